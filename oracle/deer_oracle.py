@@ -1,0 +1,471 @@
+"""Float64 CPU oracle for the GTF-DEER hot path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this module: only the tests, the smoke check and the benchmark's CPU
+baseline leg use it.  It shares no code with the HIP library; the two meet only
+through the seeded input generators (``workloads``), which hold none of the
+method's arithmetic.
+
+Everything here is plain and sequential on purpose: float64 (complex128 for the
+diagonal SSM), Python loops over time, NumPy matrix products as the only
+library primitive.  Inputs are the float32 arrays the GPU reads, promoted to
+float64 (the forcing strength alpha too is rounded through float32 first).
+
+Conventions (0-based arrays, paper indices in the comments):
+  x    [B, T+1, N]   observations x_0..x_T
+  z    [B, T, M]     states z_1..z_T (z[:, k] is z_{k+1})
+  z0   [B, M]        fixed initial state z_0
+  zt   [B, T, M]     forced states zt[:, k] = z~_k, the input of step k+1
+  mask [B, T, H]     ReLU activation pattern of step k+1 (H = M or L)
+The observation matrix is the identity read-out of the first N latents,
+B = [I_N 0] (model-setup appendix, initialisation paragraph), so the teacher
+states are zbar_t = [x_t; 0] and the projector P_alpha = I - alpha B^+ B is
+diag(1 - a) with a_i = alpha for i < N and 0 otherwise.
+
+Readings of the paper taken here (each also listed in the design notes):
+  * step 1 is unforced: z~_0 := z_0 (GTF-DEER residual definition); with the
+    default z_0 = zbar_0 both readings coincide;
+  * phi'(0) = 0, i.e. the activation mask is (u > 0) strictly;
+  * the convergence test is absolute, per sequence, on max |Delta z| over all
+    (t, m); the update is applied before the test and a converged sequence is
+    frozen; ``iters`` counts updates including the verifying one;
+  * loss = mean over the batch of the per-sequence MSE, so the seed is
+    dL/dz_t = 2/(B N T) [z_t[:N] - x_t; 0];
+  * the adjoint is exported as lam = dL/dz (= -v in the paper's sign).
+Parity unpinned: nothing.  Every function is pinned by tests/test_oracle_pins.py
+(closed forms, dense solves, brute force, finite differences and independent
+automatic differentiation); absolute Newton iteration counts of the named
+workloads have no paper value and are only reported.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+f64 = np.float64
+
+
+# --------------------------------------------------------------------------------------
+# forcing: GTF mix and error-forcing projector (eqs. GTF, error_forcing)
+# --------------------------------------------------------------------------------------
+
+def alpha_as_gpu(alpha: float) -> float:
+    """The forcing strength as the GPU sees it (float32), promoted to float64."""
+    return float(np.float32(alpha))
+
+
+def forcing_weights(M: int, n_forced: int, alpha: float) -> np.ndarray:
+    """a with P_alpha = I - alpha B^+ B = diag(1 - a) for B = [I_N 0] (eq. error_forcing)."""
+    a = np.zeros(M, f64)
+    a[:n_forced] = alpha_as_gpu(alpha)
+    return a
+
+
+def teacher_states(x: np.ndarray, M: int) -> np.ndarray:
+    """zbar_t = B^+ x_t = [x_t; 0] for t = 0..T (Alg. GTF-DEER, forcing targets)."""
+    x = np.asarray(x, f64)
+    Bn, T1, N = x.shape
+    zbar = np.zeros((Bn, T1, M), f64)
+    zbar[:, :, :N] = x
+    return zbar
+
+
+def initial_state(x: np.ndarray, M: int, z0=None) -> np.ndarray:
+    """z_0 = zbar_0 unless given (Alg. GTF-DEER initialisation)."""
+    if z0 is None:
+        return teacher_states(x[:, :1], M)[:, 0]
+    return np.asarray(z0, f64).copy()
+
+
+def forced_states(z: np.ndarray, zbar: np.ndarray, a: np.ndarray, z0: np.ndarray) -> np.ndarray:
+    """z~_{t-1} = (1 - a) z_{t-1} + a zbar_{t-1} for t >= 2 and z~_0 = z_0 (eqs. GTF,
+    error_forcing; GTF-DEER residual for step 1)."""
+    zt = np.empty_like(z)
+    zt[:, 0] = z0
+    zt[:, 1:] = (1.0 - a) * z[:, :-1] + a * zbar[:, 1:-1]
+    return zt
+
+
+# --------------------------------------------------------------------------------------
+# models: vanilla PLRNN and shallow PLRNN (eq. shplrnn_nonlinear)
+# --------------------------------------------------------------------------------------
+
+def _p(model, k):
+    return np.asarray(model[k], f64)
+
+
+def preactivation(model: dict, zt: np.ndarray) -> np.ndarray:
+    """Argument of the ReLU: z~ itself (vanilla, V = I, b = 0) or W2 z~ + h2 (shallow)."""
+    if model["kind"] == "plrnn":
+        return zt
+    return zt @ _p(model, "W2").T + _p(model, "h2")
+
+
+def model_map(model: dict, zt: np.ndarray) -> np.ndarray:
+    """F(z~) = diag(A) z~ + W relu(V z~ + b) + h (eq. shplrnn_nonlinear; no external inputs)."""
+    u = preactivation(model, zt)
+    relu = np.maximum(u, 0.0)
+    if model["kind"] == "plrnn":
+        return _p(model, "A") * zt + relu @ _p(model, "W").T + _p(model, "h")
+    return _p(model, "A") * zt + relu @ _p(model, "W1").T + _p(model, "h1")
+
+
+def activation_mask(model: dict, zt: np.ndarray) -> np.ndarray:
+    """phi'(u) for phi = ReLU, decided in float64: (u > 0)."""
+    return preactivation(model, zt) > 0.0
+
+
+def activation_mask_fp32(model: dict, z: np.ndarray, x: np.ndarray, alpha: float, n_forced: int,
+                         z0=None) -> np.ndarray:
+    """The same ReLU decision taken in float32, in the order the GPU kernels take it.
+
+    Where floating point decides an integer both sides decide in the same
+    precision.  z~ = fl(fl(p*z) + fl(a*zbar)) with p = fl(1 - a) (no fused
+    multiply-add); at step 1, z~ = z_0.  Shallow model: u = h2 + sum_j W2_ij z~_j,
+    accumulated left to right from h2 with a separate rounding after every
+    multiply and every add.
+    """
+    f = np.float32
+    z = np.asarray(z, f)
+    Bn, T, M = z.shape
+    a32 = np.zeros(M, f)
+    a32[:n_forced] = f(alpha)
+    p32 = (f(1.0) - a32).astype(f)
+    zbar = np.zeros((Bn, T + 1, M), f)
+    zbar[:, :, :x.shape[2]] = np.asarray(x, f)
+    zt = np.empty((Bn, T, M), f)
+    zt[:, 0] = zbar[:, 0] if z0 is None else np.asarray(z0, f)
+    zt[:, 1:] = (p32 * z[:, :-1]).astype(f) + (a32 * zbar[:, 1:-1]).astype(f)
+    if model["kind"] == "plrnn":
+        return zt > 0
+    W2 = np.asarray(model["W2"], f)
+    acc = np.broadcast_to(np.asarray(model["h2"], f), (Bn, T, W2.shape[0])).copy()
+    for j in range(M):
+        acc = acc + (zt[:, :, j:j + 1] * W2[:, j]).astype(f)
+    return acc > 0
+
+
+def jvp(model: dict, mask: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """J_F v with J_F = diag(A) + W diag(phi') V (model-setup appendix, Jacobian of F)."""
+    if model["kind"] == "plrnn":
+        return _p(model, "A") * v + (mask * v) @ _p(model, "W").T
+    return _p(model, "A") * v + (mask * (v @ _p(model, "W2").T)) @ _p(model, "W1").T
+
+
+def vjp(model: dict, mask: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """J_F^T w for the same Jacobian."""
+    if model["kind"] == "plrnn":
+        return _p(model, "A") * w + mask * (w @ _p(model, "W"))
+    return _p(model, "A") * w + (mask * (w @ _p(model, "W1"))) @ _p(model, "W2")
+
+
+def jacobian_dense(model: dict, mask: np.ndarray) -> np.ndarray:
+    """Dense J_F for masks [..., H]: diag(A) + W diag(m) V."""
+    A = _p(model, "A")
+    if model["kind"] == "plrnn":
+        J = _p(model, "W") * mask[..., None, :]
+    else:
+        J = (_p(model, "W1") * mask[..., None, :]) @ _p(model, "W2")
+    return J + np.diag(A)
+
+
+def forced_jacobians(model: dict, mask: np.ndarray, a: np.ndarray) -> np.ndarray:
+    """J~_t = J_F(z~_{t-1}) P_alpha (eq. error_forcing_decomp), dense [B, T, M, M]."""
+    return jacobian_dense(model, mask) * (1.0 - a)[None, :]
+
+
+# --------------------------------------------------------------------------------------
+# O1: sequential GTF rollout (Alg. initial value / trajectory matching with GTF)
+# --------------------------------------------------------------------------------------
+
+def rollout(model: dict, x: np.ndarray, alpha: float, n_forced: int, z0=None) -> np.ndarray:
+    """z_t = F(z~_{t-1}) for t = 1..T, one step at a time.  This is the unique
+    zero-residual trajectory that DEER converges to."""
+    x = np.asarray(x, f64)
+    Bn, T1, _ = x.shape
+    T = T1 - 1
+    M = np.asarray(model["A"]).shape[0]
+    a = forcing_weights(M, n_forced, alpha)
+    zbar = teacher_states(x, M)
+    zprev = initial_state(x, M, z0)
+    z = np.empty((Bn, T, M), f64)
+    for t in range(1, T + 1):
+        ztil = zprev if t == 1 else (1.0 - a) * zprev + a * zbar[:, t - 1]
+        zprev = model_map(model, ztil)
+        z[:, t - 1] = zprev
+    return z
+
+
+# --------------------------------------------------------------------------------------
+# sequential affine recurrences (the operation the associative scan evaluates)
+# --------------------------------------------------------------------------------------
+
+def affine_recurrence(apply_J, b: np.ndarray) -> np.ndarray:
+    """y_t = J_t y_{t-1} + b_t for t = 1..T with y_0 = 0 (eq. DEER_update as a linear
+    recursion).  apply_J(k, v) returns J_{k+1} v for every batch row."""
+    Bn, T, M = b.shape
+    out = np.empty_like(b)
+    prev = np.zeros((Bn, M), b.dtype)
+    for k in range(T):
+        prev = apply_J(k, prev) + b[:, k]
+        out[:, k] = prev
+    return out
+
+
+def reverse_affine_recurrence(apply_JT, g: np.ndarray) -> np.ndarray:
+    """l_T = g_T and l_{t-1} = J_t^T l_t + g_{t-1} for t = T..2 (eq. backward_recursion).
+    apply_JT(k, w) returns J_{k+1}^T w for every batch row."""
+    Bn, T, M = g.shape
+    out = np.empty_like(g)
+    nxt = g[:, T - 1].copy()
+    out[:, T - 1] = nxt
+    for k in range(T - 2, -1, -1):      # l_{k+1} (array index k) uses J_{k+2}
+        nxt = apply_JT(k + 1, nxt) + g[:, k]
+        out[:, k] = nxt
+    return out
+
+
+# --------------------------------------------------------------------------------------
+# O2: explicit GTF-DEER Newton loop (Alg. GTF-DEER; eq. GTF_DEER_update)
+# --------------------------------------------------------------------------------------
+
+def residual_and_masks(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, z0=None):
+    """r_t = z_t - F(z~_{t-1}) (eq. GTF_residual) together with F and the masks at z~."""
+    x = np.asarray(x, f64)
+    z = np.asarray(z, f64)
+    M = z.shape[2]
+    a = forcing_weights(M, n_forced, alpha)
+    zbar = teacher_states(x, M)
+    zt = forced_states(z, zbar, a, initial_state(x, M, z0))
+    F = model_map(model, zt)
+    return z - F, F, activation_mask(model, zt), zt
+
+
+def newton(model: dict, x: np.ndarray, alpha: float, n_forced: int, *, z0=None, init: str = "teacher",
+           z_init=None, tol: float = 1e-5, max_iter: int = 500, fixed_iters: int = 0, history: bool = False):
+    """GTF-DEER forward solve.  Each update linearises at z^(k): Delta_t =
+    J~_t Delta_{t-1} - r_t, Delta_0 = 0, solved here by the sequential recursion,
+    then z^(k+1) = z^(k) + Delta.  Returns dict(z, iters, norms, status[, history])."""
+    x = np.asarray(x, f64)
+    Bn, T1, _ = x.shape
+    T = T1 - 1
+    M = np.asarray(model["A"]).shape[0]
+    a = forcing_weights(M, n_forced, alpha)
+    p = 1.0 - a
+    zbar = teacher_states(x, M)
+    z0v = initial_state(x, M, z0)
+    if init == "teacher":
+        z = zbar[:, 1:].copy()
+    elif init == "zero":
+        z = np.zeros((Bn, T, M), f64)
+    elif init == "user":
+        z = np.asarray(z_init, f64).copy()
+    else:
+        raise ValueError(init)
+    active = np.ones(Bn, bool)
+    iters = np.zeros(Bn, np.int64)
+    norms = np.full(Bn, np.nan)
+    nonfinite = np.zeros(Bn, bool)
+    hist = [z.copy()] if history else None
+    k = 0
+    while True:
+        if fixed_iters > 0:
+            if k == fixed_iters:
+                break
+        elif not active.any() or k == max_iter:
+            break
+        zt = forced_states(z, zbar, a, z0v)
+        r = z - model_map(model, zt)
+        mask = activation_mask(model, zt)
+        delta = affine_recurrence(lambda kk, v: jvp(model, mask[:, kk], p * v), -r)
+        e = np.abs(delta).reshape(Bn, -1).max(axis=1) if T > 0 else np.zeros(Bn)
+        e = np.where(np.isnan(delta).reshape(Bn, -1).any(axis=1), np.nan, e)
+        upd = active if fixed_iters == 0 else np.ones(Bn, bool)
+        z[upd] += delta[upd]
+        iters[upd] += 1
+        norms[upd] = e[upd]
+        bad = upd & ~np.isfinite(e)
+        nonfinite |= bad
+        if fixed_iters == 0:
+            active &= ~((e < tol) | bad)
+        if history:
+            hist.append(z.copy())
+        k += 1
+    status = "ok"
+    if nonfinite.any():
+        status = "nonfinite"
+    elif fixed_iters == 0 and active.any():
+        status = "not_converged"
+    out = {"z": z, "iters": iters, "norms": norms, "status": status}
+    if history:
+        out["history"] = hist
+    return out
+
+
+# --------------------------------------------------------------------------------------
+# O3: loss seed, IFT adjoint and parameter gradients (gradients appendix)
+# --------------------------------------------------------------------------------------
+
+def mse_loss(z: np.ndarray, x: np.ndarray) -> float:
+    """Batch mean of (1/(N T)) sum_t ||x_t - B z_t||^2 (eq. mse_loss_series)."""
+    z = np.asarray(z, f64)
+    x = np.asarray(x, f64)
+    Bn, T, _ = z.shape
+    N = x.shape[2]
+    return float(((z[:, :, :N] - x[:, 1:]) ** 2).sum() / (Bn * N * T))
+
+
+def mse_seed(z: np.ndarray, x: np.ndarray) -> np.ndarray:
+    """dL/dz_t = 2/(B N T) B^T (B z_t - x_t), t = 1..T."""
+    z = np.asarray(z, f64)
+    x = np.asarray(x, f64)
+    Bn, T, M = z.shape
+    N = x.shape[2]
+    g = np.zeros((Bn, T, M), f64)
+    g[:, :, :N] = 2.0 / (Bn * N * T) * (z[:, :, :N] - x[:, 1:])
+    return g
+
+
+def _masks_at(model, x, z, alpha, n_forced, z0, mask_precision):
+    r, F, mask64, zt = residual_and_masks(model, x, z, alpha, n_forced, z0)
+    if mask_precision == "float32":
+        mask = activation_mask_fp32(model, z, x, alpha, n_forced, z0)
+    elif mask_precision == "float64":
+        mask = mask64
+    else:
+        raise ValueError(mask_precision)
+    return mask, zt
+
+
+def adjoint(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, *, z0=None,
+            g=None, mask_precision: str = "float64") -> np.ndarray:
+    """lam = dL/dz by the backward recursion lam_T = g_T, lam_{t-1} = J~_t^T lam_t + g_{t-1}
+    (eqs. adjoint_eq, backward_recursion with lam = -v).  J~_t is taken at z~_{t-1} of
+    the given trajectory z (normally the converged one)."""
+    z = np.asarray(z, f64)
+    M = z.shape[2]
+    p = 1.0 - forcing_weights(M, n_forced, alpha)
+    mask, _ = _masks_at(model, x, z, alpha, n_forced, z0, mask_precision)
+    g = mse_seed(z, x) if g is None else np.asarray(g, f64)
+    # J~^T w = P_alpha J_F^T w
+    return reverse_affine_recurrence(lambda k, w: p * vjp(model, mask[:, k], w), g)
+
+
+def param_grads(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, lam: np.ndarray, *,
+                z0=None, mask_precision: str = "float64") -> dict:
+    """dL/dtheta = sum_t lam_t^T dF(z~_{t-1})/dtheta (gradients appendix, IFT summary),
+    summed directly over every (b, t) in float64."""
+    z = np.asarray(z, f64)
+    lam = np.asarray(lam, f64)
+    mask, zt = _masks_at(model, x, z, alpha, n_forced, z0, mask_precision)
+    out = {"A": np.einsum("bti,bti->i", lam, zt)}
+    if model["kind"] == "plrnn":
+        relu = np.where(mask, zt, 0.0)
+        out["W"] = np.einsum("bti,btj->ij", lam, relu)
+        out["h"] = lam.sum(axis=(0, 1))
+    else:
+        u = preactivation(model, zt)
+        relu = np.where(mask, u, 0.0)
+        delta = (lam @ _p(model, "W1")) * mask
+        out["W1"] = np.einsum("bti,btl->il", lam, relu)
+        out["W2"] = np.einsum("btl,btj->lj", delta, zt)
+        out["h1"] = lam.sum(axis=(0, 1))
+        out["h2"] = delta.sum(axis=(0, 1))
+    return out
+
+
+# --------------------------------------------------------------------------------------
+# O4: residual, masks and forced Jacobians at a given trajectory
+# --------------------------------------------------------------------------------------
+
+def jacobian_at(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, *, z0=None,
+                mask_precision: str = "float64", dense_index=None) -> dict:
+    """F, r, masks and (for the (b, t) pairs in dense_index) dense J~_t at trajectory z."""
+    r, F, mask64, zt = residual_and_masks(model, x, z, alpha, n_forced, z0)
+    mask = mask64 if mask_precision == "float64" else activation_mask_fp32(model, z, x, alpha, n_forced, z0)
+    out = {"F": F, "r": r, "mask": mask, "zt": zt}
+    if dense_index is not None:
+        M = z.shape[2]
+        a = forcing_weights(M, n_forced, alpha)
+        out["J"] = np.stack([forced_jacobians(model, mask[b, t], a) for (b, t) in dense_index])
+    return out
+
+
+# --------------------------------------------------------------------------------------
+# O5: diagonal complex SSM (eq. shplrnn_ssm with diagonal complex A; Alg. LSSM)
+# --------------------------------------------------------------------------------------
+
+def diag_scan(lam: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """h_t = lam * h_{t-1} + b_t, h_0 = 0, t = 1..T, complex128."""
+    lam = np.asarray(lam, np.complex128)
+    b = np.asarray(b, np.complex128)
+    h = np.empty_like(b)
+    prev = np.zeros(b.shape[:1] + b.shape[2:], np.complex128)
+    for k in range(b.shape[1]):
+        prev = lam * prev + b[:, k]
+        h[:, k] = prev
+    return h
+
+
+def diag_scan_reverse(lam: np.ndarray, g: np.ndarray) -> np.ndarray:
+    """a_T = g_T and a_{t-1} = conj(lam) * a_t + g_{t-1}: the transpose of diag_scan
+    with the complex plane read as R^2 (the 2x2 block [[p,-q],[q,p]] transposes to
+    multiplication by conj(lam))."""
+    lam = np.asarray(lam, np.complex128)
+    g = np.asarray(g, np.complex128)
+    out = np.empty_like(g)
+    nxt = np.zeros(g.shape[:1] + g.shape[2:], np.complex128)
+    for k in range(g.shape[1] - 1, -1, -1):
+        nxt = np.conj(lam) * nxt + g[:, k]
+        out[:, k] = nxt
+    return out
+
+
+def diag_ssm_inputs(params: dict, x: np.ndarray) -> np.ndarray:
+    """b_t = Bc u_t with u_t = x_{t-1} (teacher input of the LSSM), t = 1..T."""
+    u = np.asarray(x, f64)[:, :-1]
+    return u @ np.asarray(params["Bc"], np.complex128).T
+
+
+def diag_ssm_readout(params: dict, h: np.ndarray) -> np.ndarray:
+    """y_t = Wb relu(Wa Re(h_t) + ca) + cb (one-hidden-layer MLP read-out)."""
+    s = np.real(h) @ np.asarray(params["Wa"], f64).T + np.asarray(params["ca"], f64)
+    return np.maximum(s, 0.0) @ np.asarray(params["Wb"], f64).T + np.asarray(params["cb"], f64)
+
+
+def diag_ssm_loss_and_seed(params: dict, h: np.ndarray, x: np.ndarray):
+    """MSE of the read-out against x_{1:T} and g = dL/dRe(h) (chain rule through the MLP)."""
+    x = np.asarray(x, f64)
+    Bn, T, _ = h.shape
+    No = x.shape[2]
+    Wa = np.asarray(params["Wa"], f64)
+    Wb = np.asarray(params["Wb"], f64)
+    s = np.real(h) @ Wa.T + np.asarray(params["ca"], f64)
+    y = np.maximum(s, 0.0) @ Wb.T + np.asarray(params["cb"], f64)
+    err = y - x[:, 1:]
+    loss = float((err ** 2).sum() / (Bn * No * T))
+    dy = 2.0 / (Bn * No * T) * err
+    ds = (dy @ Wb) * (s > 0.0)
+    g = ds @ Wa
+    grads = {"Wb": np.einsum("bto,btk->ok", dy, np.maximum(s, 0.0)), "cb": dy.sum(axis=(0, 1)),
+             "Wa": np.einsum("btk,btn->kn", ds, np.real(h)), "ca": ds.sum(axis=(0, 1))}
+    return loss, g, grads
+
+
+def diag_ssm_param_grads(a_adj: np.ndarray, h: np.ndarray, x: np.ndarray) -> dict:
+    """dlam = sum_t a_t conj(h_{t-1}) and dBc = sum_t a_t u_t^T (u_t = x_{t-1}), the
+    complex gradients d/dRe + i d/dIm."""
+    hprev = np.concatenate([np.zeros_like(h[:, :1]), h[:, :-1]], axis=1)
+    u = np.asarray(x, f64)[:, :-1]
+    return {"lam": (a_adj * np.conj(hprev)).sum(axis=(0, 1)),
+            "Bc": np.einsum("btn,btk->nk", a_adj, u)}
+
+
+def diag_ssm_step(params: dict, x: np.ndarray) -> dict:
+    """Forward scan, read-out loss, reverse scan and all gradients of the diagonal SSM."""
+    b = diag_ssm_inputs(params, x)
+    h = diag_scan(params["lam"], b)
+    loss, g, mlp_grads = diag_ssm_loss_and_seed(params, h, x)
+    a_adj = diag_scan_reverse(params["lam"], g.astype(np.complex128))
+    grads = diag_ssm_param_grads(a_adj, h, x)
+    grads.update(mlp_grads)
+    return {"b": b, "h": h, "loss": loss, "g": g, "a": a_adj, "grads": grads}

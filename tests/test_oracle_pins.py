@@ -1,0 +1,432 @@
+"""Pins of the float64 oracle against facts that do not come from the oracle.
+
+Each test names the passage or mathematical fact it relies on.  The paper
+prints no worked numerical example, so the pins are closed forms, textbook
+routines (LAPACK dense solves, SVD), brute force over tiny sizes, central
+finite differences and independent automatic differentiation (torch, CPU,
+float64) of the sequential rollout.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle as O
+from oracle import brute
+from workloads import plrnn_params, shplrnn_params, random_plrnn_case, random_shplrnn_case
+
+torch = pytest.importorskip("torch")
+
+
+def _vanilla(M, seed, w_std=0.3, a_range=(0.5, 0.9)):
+    p = plrnn_params(M, np.random.default_rng(seed), a_range=a_range, w_std=w_std)
+    return {"kind": "plrnn", **p}
+
+
+def _shallow(M, L, seed):
+    p = shplrnn_params(M, L, np.random.default_rng(seed))
+    return {"kind": "shplrnn", **p}
+
+
+def _x(B, T, N, seed):
+    return np.random.default_rng(seed).standard_normal((B, T + 1, N)).astype(np.float32)
+
+
+# ------------------------------------------------------------------------------------
+# F itself: special cases with a closed form (eq. shplrnn_nonlinear)
+# ------------------------------------------------------------------------------------
+
+def test_model_map_permutation_closed_form():
+    """With A = 0, h = 0 and W a permutation matrix, F(z)_i = relu(z_pi(i)); a transposed
+    W would give relu(z_pi^-1(i)) instead (pi is a 3-cycle, not an involution)."""
+    pi = np.array([1, 2, 0, 4, 3])
+    W = np.zeros((5, 5), np.float32)
+    W[np.arange(5), pi] = 1.0
+    m = {"kind": "plrnn", "A": np.zeros(5, np.float32), "W": W, "h": np.zeros(5, np.float32)}
+    z = np.array([[1.5, -2.0, 0.25, -0.5, 3.0]])
+    F = O.model_map(m, z)
+    assert np.array_equal(F[0], np.maximum(z[0, pi], 0.0))
+    m2 = dict(m, A=np.array([0.5, 0.5, 0.5, 0.5, 0.5], np.float32), h=np.arange(5, dtype=np.float32))
+    assert np.allclose(O.model_map(m2, z)[0], 0.5 * z[0] + np.maximum(z[0, pi], 0.0) + np.arange(5))
+
+
+def test_shallow_map_permutation_closed_form():
+    """Shallow PLRNN with W2 = permutation, W1 = I, h2 = 0: F = A z + relu(z_pi) + h1;
+    with W2 = I, W1 = permutation: F = A z + relu(z)_pi + h1 (pi a 3-cycle)."""
+    M = 3
+    pi = np.array([2, 0, 1])
+    P = np.zeros((M, M), np.float32)
+    P[np.arange(M), pi] = 1.0
+    A = np.array([0.1, 0.2, 0.3], np.float32)
+    h1 = np.array([1.0, -1.0, 0.5], np.float32)
+    z = np.array([[0.7, -1.2, 2.0]])
+    m = {"kind": "shplrnn", "A": A, "W1": np.eye(M, dtype=np.float32), "W2": P, "h1": h1,
+         "h2": np.zeros(M, np.float32)}
+    assert np.allclose(O.model_map(m, z)[0], A * z[0] + np.maximum(z[0, pi], 0) + h1)
+    m = dict(m, W1=P, W2=np.eye(M, dtype=np.float32))
+    assert np.allclose(O.model_map(m, z)[0], A * z[0] + np.maximum(z[0], 0)[pi] + h1)
+    m = dict(m, h2=np.array([-10.0, 10.0, 0.0], np.float32))   # hidden biases shift the kinks
+    assert np.allclose(O.model_map(m, z)[0], A * z[0] + np.maximum(z[0] + m["h2"], 0)[pi] + h1)
+
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+def test_jacobian_matches_finite_differences(kind):
+    """J_F = diag(A) + W diag(phi'(Vz+b)) V (model-setup appendix) against central
+    differences of F at points away from the ReLU kinks (F is linear on each cell)."""
+    rng = np.random.default_rng(3)
+    m = _vanilla(6, 1) if kind == "plrnn" else _shallow(5, 12, 2)
+    for _ in range(5):
+        z = rng.standard_normal((1, m["A"].shape[0]))
+        u = O.preactivation(m, z)
+        assume = np.abs(u).min() > 1e-3
+        if not assume:
+            continue
+        J = O.jacobian_dense(m, O.activation_mask(m, z))[0]
+        eps = 1e-6
+        Jfd = np.empty_like(J)
+        for j in range(z.shape[1]):
+            e = np.zeros_like(z)
+            e[0, j] = eps
+            Jfd[:, j] = (O.model_map(m, z + e) - O.model_map(m, z - e))[0] / (2 * eps)
+        assert np.allclose(J, Jfd, atol=1e-8)
+        v = rng.standard_normal((1, z.shape[1]))
+        mask = O.activation_mask(m, z)
+        assert np.allclose(O.jvp(m, mask, v)[0], J @ v[0])
+        assert np.allclose(O.vjp(m, mask, v)[0], J.T @ v[0])
+
+
+def test_forcing_projector_is_identity_readout():
+    """P_alpha = I - alpha B^+ B with B = [I_N 0]: B^+ = B^T, so P_alpha = diag(1-a)
+    (eq. error_forcing); checked against numpy's pseudo-inverse."""
+    M, N, alpha = 7, 3, 0.3
+    Bm = np.hstack([np.eye(N), np.zeros((N, M - N))])
+    P = np.eye(M) - O.alpha_as_gpu(alpha) * np.linalg.pinv(Bm) @ Bm
+    assert np.allclose(P, np.diag(1.0 - O.forcing_weights(M, N, alpha)))
+    x = _x(2, 4, N, 0)
+    zbar = O.teacher_states(x, M)
+    assert np.allclose(zbar, np.einsum("mn,btn->btm", np.linalg.pinv(Bm), x))
+
+
+# ------------------------------------------------------------------------------------
+# P1: the affine recurrence, its transpose and the scan decomposition
+# ------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T", [1, 2, 3, 7, 16])
+def test_affine_recurrence_equals_block_bidiagonal_solve(T):
+    """y_t = J_t y_{t-1} + b_t is the solution of the block-bidiagonal system of
+    eq. blockdiag_jacobian; its transpose solves the adjoint system (eq. adjoint_eq)."""
+    rng = np.random.default_rng(T)
+    M = 3
+    J = rng.standard_normal((T, M, M)) * 0.7
+    b = rng.standard_normal((T, M))
+    y = O.affine_recurrence(lambda k, v: v @ J[k].T, b[None])[0]
+    assert np.allclose(y, brute.block_bidiagonal_solve(J, b), rtol=1e-12, atol=1e-12)
+    g = rng.standard_normal((T, M))
+    lam = O.reverse_affine_recurrence(lambda k, w: w @ J[k], g[None])[0]
+    assert np.allclose(lam, brute.block_bidiagonal_adjoint_solve(J, g), rtol=1e-12, atol=1e-12)
+    # transpose identity <g, S b> = <S^T g, b>
+    assert np.isclose((g * y).sum(), (lam * b).sum(), rtol=1e-12)
+
+
+@pytest.mark.parametrize("T", [1, 2, 4, 6, 8])
+def test_every_bracketing_gives_the_same_map(T):
+    """Associativity of (A2, b2) o (A1, b1) = (A2 A1, A2 b1 + b2) (scheduled-sampling
+    appendix): every bracketing equals the sequential fold; its b is y_T."""
+    rng = np.random.default_rng(10 + T)
+    M = 2
+    J = rng.standard_normal((T, M, M))
+    b = rng.standard_normal((T, M))
+    elems = [(J[k], b[k]) for k in range(T)]
+    y = O.affine_recurrence(lambda k, v: v @ J[k].T, b[None])[0]
+    Pseq = np.eye(M)
+    for k in range(T):
+        Pseq = J[k] @ Pseq
+    for P, v in brute.all_bracketings(elems):
+        assert np.allclose(P, Pseq, rtol=1e-12, atol=1e-12)
+        assert np.allclose(v, y[-1], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("T", [1, 5, 16])
+def test_chunked_scan_equals_recurrence_for_every_chunk(T):
+    rng = np.random.default_rng(20 + T)
+    M = 4
+    J = rng.standard_normal((T, M, M)) * 0.5
+    b = rng.standard_normal((T, M))
+    y = O.affine_recurrence(lambda k, v: v @ J[k].T, b[None])[0]
+    for C in range(1, T + 1):
+        assert np.allclose(brute.chunked_scan(J, b, C), y, rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------------------------------------
+# P2/P3/P6: Newton reaches the rollout; prefix exactness; finite termination
+# ------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("kind,M,N,alpha", [("plrnn", 4, 3, 0.2), ("plrnn", 3, 3, 0.1), ("plrnn", 16, 3, 0.2),
+                                            ("shplrnn", 5, 5, 0.1), ("shplrnn", 6, 2, 0.3)])
+def test_newton_converges_to_rollout(kind, M, N, alpha):
+    """The zero of the GTF residual is the sequential GTF rollout (DEER section and
+    GTF-DEER residual); Newton in float64 with eps = 1e-13 reaches it to 1e-11."""
+    m = _vanilla(M, 5) if kind == "plrnn" else _shallow(M, 3 * M, 6)
+    x = _x(3, 60, N, 7)
+    ref = O.rollout(m, x, alpha, N)
+    res = O.newton(m, x, alpha, N, tol=1e-13, max_iter=200)
+    assert res["status"] == "ok"
+    assert np.abs(res["z"] - ref).max() <= 1e-11
+    zr = O.rollout(m, x, alpha, N, z0=np.ones((3, M)))     # user initial state
+    rz = O.newton(m, x, alpha, N, z0=np.ones((3, M)), init="zero", tol=1e-13, max_iter=200)
+    assert np.abs(rz["z"] - zr).max() <= 1e-11
+
+
+def test_rollout_residual_is_zero():
+    m = _vanilla(5, 8)
+    x = _x(2, 30, 3, 9)
+    z = O.rollout(m, x, 0.3, 3)
+    r, _, _, _ = O.residual_and_masks(m, x, z, 0.3, 3)
+    assert np.abs(r).max() < 1e-13
+
+
+@pytest.mark.parametrize("init", ["teacher", "zero"])
+def test_newton_prefix_exactness(init):
+    """With Delta_0 = 0 and z_0 fixed, after k updates z_1..z_k are exact (eq. DEER_update
+    read step by step); hence termination within T updates plus the verifying one."""
+    m = _vanilla(3, 11, w_std=0.8)
+    T = 12
+    x = _x(2, T, 3, 12)
+    ref = O.rollout(m, x, 0.0, 3)
+    res = O.newton(m, x, 0.0, 3, init=init, fixed_iters=T, history=True)
+    for k, zk in enumerate(res["history"]):
+        if k == 0:
+            continue
+        assert np.abs(zk[:, :k] - ref[:, :k]).max() < 1e-12, k
+    full = O.newton(m, x, 0.0, 3, init=init, tol=1e-12, max_iter=100)
+    assert full["iters"].max() <= T + 1
+
+
+def test_newton_lands_on_fixed_point_once_masks_match():
+    """F is affine on each activation cell, so a Newton update linearised at an iterate
+    that shares the fixed point's masks is exact: one update from a small perturbation
+    of z* returns z* (pins J~_t = J_F(z~) P_alpha: any other matrix leaves an error)."""
+    m = _vanilla(6, 13)
+    x = _x(2, 40, 4, 14)
+    alpha = 0.25
+    zs = O.rollout(m, x, alpha, 4)
+    _, _, mask_s, zt_s = O.residual_and_masks(m, x, zs, alpha, 4)
+    pert = 1e-7 * np.random.default_rng(1).standard_normal(zs.shape)
+    z1 = zs + pert
+    _, _, mask1, _ = O.residual_and_masks(m, x, z1, alpha, 4)
+    assert np.array_equal(mask1, mask_s), "perturbation crossed a kink; choose a smaller one"
+    res = O.newton(m, x, alpha, 4, init="user", z_init=z1, fixed_iters=1)
+    assert np.abs(res["z"] - zs).max() < 1e-13
+    res2 = O.newton(m, x, alpha, 4, init="user", z_init=z1, tol=1e-10)
+    assert res2["iters"].tolist() == [2, 2]
+
+
+# ------------------------------------------------------------------------------------
+# P4/P5: alpha = 0 on a linear model; alpha = 1 reproduces the data-driven states
+# ------------------------------------------------------------------------------------
+
+def test_alpha0_linear_model_closed_form_and_two_iterations():
+    """W = 0: z_t = A^t z_0 + (1 - A^t)/(1 - A) h, and DEER needs exactly 2 updates
+    (the first exact, the second verifying; footnote to the runtime section)."""
+    M, T = 4, 50
+    A = np.array([0.5, 0.7, 0.9, 0.95], np.float32)
+    h = np.array([0.1, -0.2, 0.3, 0.05], np.float32)
+    m = {"kind": "plrnn", "A": A, "W": np.zeros((M, M), np.float32), "h": h}
+    x = _x(2, T, M, 15)
+    z0 = x[:, 0].astype(np.float64)
+    t = np.arange(1, T + 1)[None, :, None]
+    A64, h64 = A.astype(np.float64), h.astype(np.float64)
+    closed = A64 ** t * z0[:, None, :] + (1 - A64 ** t) / (1 - A64) * h64
+    res = O.newton(m, x, 0.0, M, tol=1e-10)
+    assert np.abs(res["z"] - closed).max() < 1e-12
+    assert res["iters"].tolist() == [2, 2]
+    assert np.abs(O.rollout(m, x, 0.0, M) - closed).max() < 1e-12
+
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+def test_alpha1_full_observation_closed_form(kind):
+    """alpha = 1 and M <= N: z~ = zbar, J~ = 0, so z*_t = F(zbar_{t-1}) in closed form and
+    DEER stops after 2 updates."""
+    M = 4
+    m = _vanilla(M, 16, w_std=1.0) if kind == "plrnn" else _shallow(M, 9, 17)
+    x = _x(3, 25, M, 18)
+    xb = x.astype(np.float64)
+    closed = O.model_map(m, xb[:, :-1])
+    res = O.newton(m, x, 1.0, M, tol=1e-10)
+    assert np.abs(res["z"] - closed).max() < 1e-13
+    assert res["iters"].tolist() == [2, 2, 2]
+
+
+def test_prop1_contraction_bound():
+    """Prop. 1 (M <= N): J~_t = (1 - alpha) J_F, so ||J~_t||_2 <= (1 - alpha) sigma~_max and
+    products of k forced Jacobians are bounded by rho^k.  sigma~_max is exact here: a
+    vanilla PLRNN with M = 3 has only 2^3 distinct Jacobians."""
+    M = 3
+    m = _vanilla(M, 19, w_std=1.2)
+    sig = max(np.linalg.svd(O.jacobian_dense(m, np.array(mk, bool)), compute_uv=False)[0]
+              for mk in itertools.product([0, 1], repeat=M))
+    assert sig > 1.0
+    alpha = 1.0 - 1.0 / sig + 0.05
+    rho = (1.0 - O.alpha_as_gpu(alpha)) * sig
+    assert rho < 1.0
+    x = _x(1, 80, M, 20)
+    z = O.rollout(m, x, alpha, M)
+    _, _, mask, _ = O.residual_and_masks(m, x, z, alpha, M)
+    Jt = O.forced_jacobians(m, mask[0], O.forcing_weights(M, M, alpha))
+    for k in range(80):
+        assert np.linalg.svd(Jt[k], compute_uv=False)[0] <= rho * (1 + 1e-12)
+    P = np.eye(M)
+    for k in range(80):
+        P = Jt[k] @ P
+        assert np.linalg.norm(P, 2) <= rho ** (k + 1) * (1 + 1e-9)
+
+
+# ------------------------------------------------------------------------------------
+# P8/P9: adjoint and parameter gradients
+# ------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+def test_adjoint_equals_dense_adjoint_solve(kind):
+    """lam solves R^T lam = dL/dz for R = dR/dz (eq. blockdiag_jacobian, eq. adjoint_eq)."""
+    M, N, T, alpha = 4, 2, 14, 0.3
+    m = _vanilla(M, 21) if kind == "plrnn" else _shallow(M, 8, 22)
+    x = _x(1, T, N, 23)
+    z = O.rollout(m, x, alpha, N)
+    _, _, mask, _ = O.residual_and_masks(m, x, z, alpha, N)
+    J = O.forced_jacobians(m, mask[0], O.forcing_weights(M, N, alpha))
+    g = O.mse_seed(z, x)[0]
+    lam = O.adjoint(m, x, z, alpha, N)[0]
+    assert np.allclose(lam, brute.block_bidiagonal_adjoint_solve(J, g), rtol=1e-12, atol=1e-14)
+
+
+def _torch_bptt(m, x, alpha, N):
+    """Independent reverse-mode AD (torch, float64) through the sequential GTF rollout
+    of Alg. 2 and the MSE loss: the BPTT gradient the IFT gradient must equal."""
+    t = lambda a: torch.tensor(np.asarray(a, np.float64), requires_grad=True)
+    P = {k: t(v) for k, v in m.items() if k != "kind"}
+    xt = torch.tensor(np.asarray(x, np.float64))
+    Bn, T1, _ = x.shape
+    M = P["A"].shape[0]
+    a = torch.zeros(M, dtype=torch.float64)
+    a[:N] = float(np.float32(alpha))
+    zbar = torch.zeros(Bn, T1, M, dtype=torch.float64)
+    zbar[:, :, :N] = xt
+    prev = zbar[:, 0]
+    loss = 0.0
+    for k in range(1, T1):
+        zt = prev if k == 1 else (1 - a) * prev + a * zbar[:, k - 1]
+        if m["kind"] == "plrnn":
+            prev = P["A"] * zt + torch.relu(zt) @ P["W"].T + P["h"]
+        else:
+            prev = P["A"] * zt + torch.relu(zt @ P["W2"].T + P["h2"]) @ P["W1"].T + P["h1"]
+        loss = loss + ((prev[:, :N] - xt[:, k]) ** 2).sum()
+    loss = loss / (Bn * N * (T1 - 1))
+    loss.backward()
+    return float(loss.detach()), {k: v.grad.numpy() for k, v in P.items()}
+
+
+@pytest.mark.parametrize("kind,M,N,alpha", [("plrnn", 5, 3, 0.2), ("plrnn", 3, 3, 0.1), ("shplrnn", 4, 4, 0.15),
+                                            ("shplrnn", 6, 2, 0.3)])
+def test_ift_gradient_equals_bptt(kind, M, N, alpha):
+    """The IFT gradient at the fixed point equals BPTT through the sequential rollout
+    (gradients appendix vs Alg. 2)."""
+    m = _vanilla(M, 31) if kind == "plrnn" else _shallow(M, 10, 32)
+    x = _x(2, 40, N, 33)
+    z = O.newton(m, x, alpha, N, tol=1e-13)["z"]
+    loss_ref, gref = _torch_bptt(m, x, alpha, N)
+    assert np.isclose(O.mse_loss(z, x), loss_ref, rtol=1e-12)
+    lam = O.adjoint(m, x, z, alpha, N)
+    g = O.param_grads(m, x, z, alpha, N, lam)
+    for k, v in gref.items():
+        assert np.allclose(g[k], v, rtol=1e-10, atol=1e-13), k
+
+
+def test_param_grads_central_differences():
+    """dL/dtheta of L(z*(theta)) by central differences (float64, h = 1e-6) for a few
+    entries of every parameter, at a trajectory with no activation near zero."""
+    m = _vanilla(3, 41)
+    x = _x(1, 30, 2, 42)
+    alpha = 0.2
+    z = O.rollout(m, x, alpha, 2)
+    _, _, _, zt = O.residual_and_masks(m, x, z, alpha, 2)
+    assert np.abs(zt[:, 1:]).min() > 1e-4     # z~_0 = z_0 is data, independent of theta
+    g = O.param_grads(m, x, z, alpha, 2, O.adjoint(m, x, z, alpha, 2))
+    mf = {k: (np.asarray(v, np.float64) if k != "kind" else v) for k, v in m.items()}
+    for name, idx in [("A", (1,)), ("W", (0, 2)), ("W", (2, 1)), ("h", (0,))]:
+        hstep = 1e-6
+        mp = {k: (v.copy() if k != "kind" else v) for k, v in mf.items()}
+        mm = {k: (v.copy() if k != "kind" else v) for k, v in mf.items()}
+        mp[name][idx] += hstep
+        mm[name][idx] -= hstep
+        fd = (O.mse_loss(O.rollout(mp, x, alpha, 2), x) - O.mse_loss(O.rollout(mm, x, alpha, 2), x)) / (2 * hstep)
+        assert np.isclose(g[name][idx], fd, rtol=1e-6, atol=1e-10), (name, idx)
+
+
+def test_fp32_mask_decision_agrees_away_from_ties():
+    """The float32 ReLU decision (kernel precision) equals the float64 one wherever the
+    pre-activation is not within float32 rounding of zero."""
+    for case in [random_plrnn_case(8, 3, 2, 200, 0.2, 50), random_shplrnn_case(6, 20, 6, 2, 100, 0.1, 51)]:
+        m = {"kind": case.kind, **case.params}
+        z = O.rollout(m, case.x, case.alpha, case.n_obs).astype(np.float32)
+        _, _, mask64, zt = O.residual_and_masks(m, case.x, z, case.alpha, case.n_obs)
+        u = O.preactivation(m, zt)
+        m32 = O.activation_mask_fp32(m, z, case.x, case.alpha, case.n_obs)
+        far = np.abs(u) > 1e-5 * (1 + np.abs(u).max())
+        assert np.array_equal(m32[far], mask64[far])
+
+
+# ------------------------------------------------------------------------------------
+# P10: diagonal complex SSM
+# ------------------------------------------------------------------------------------
+
+def test_diag_scan_closed_forms():
+    """Impulse response h_t = lam^(t-1) b_1 and constant input h_t = (1 - lam^t)/(1 - lam) b
+    (linear-SSM appendix: dz_t/dz_r = A^(t-r))."""
+    rng = np.random.default_rng(60)
+    lam = 0.97 * np.exp(1j * rng.uniform(0, np.pi / 10, 5))
+    T = 200
+    b = np.zeros((1, T, 5), np.complex128)
+    b[0, 0] = 1.0 + 0.5j
+    h = O.diag_scan(lam, b)
+    t = np.arange(T)[:, None]
+    assert np.allclose(h[0], lam ** t * (1.0 + 0.5j), rtol=1e-12, atol=1e-14)
+    c = rng.standard_normal(5) + 1j * rng.standard_normal(5)
+    h = O.diag_scan(lam, np.broadcast_to(c, (1, T, 5)))
+    tt = np.arange(1, T + 1)[:, None]
+    assert np.allclose(h[0], (1 - lam ** tt) / (1 - lam) * c, rtol=1e-11)
+    g = rng.standard_normal((1, T, 5)) + 1j * rng.standard_normal((1, T, 5))
+    a = O.diag_scan_reverse(lam, g)
+    bb = rng.standard_normal((1, T, 5)) + 1j * rng.standard_normal((1, T, 5))
+    # real inner product on C = R^2: <g, S b> = <S^T g, b>
+    assert np.isclose(np.real(np.conj(g) * O.diag_scan(lam, bb)).sum(), np.real(np.conj(a) * bb).sum(), rtol=1e-11)
+
+
+def test_diag_ssm_gradients_match_autograd():
+    """Gradients of the diagonal SSM training loss (scan, MLP read-out, MSE) against torch
+    autograd with lam and Bc parametrised by their real and imaginary parts."""
+    from workloads import diag_ssm_params
+    prm = diag_ssm_params(6, 3, 8, 3, np.random.default_rng(70))
+    x = _x(2, 50, 3, 71)
+    out = O.diag_ssm_step(prm, x)
+    t = lambda a: torch.tensor(np.asarray(a, np.float64), requires_grad=True)
+    lr, li = t(prm["lam"].real), t(prm["lam"].imag)
+    br, bi = t(prm["Bc"].real), t(prm["Bc"].imag)
+    Wa, ca, Wb, cb = t(prm["Wa"]), t(prm["ca"]), t(prm["Wb"]), t(prm["cb"])
+    xt = torch.tensor(x.astype(np.float64))
+    Bn, T1, _ = x.shape
+    hr = torch.zeros(Bn, 6, dtype=torch.float64)
+    hi = torch.zeros(Bn, 6, dtype=torch.float64)
+    loss = 0.0
+    for k in range(1, T1):
+        u = xt[:, k - 1]
+        hr, hi = lr * hr - li * hi + u @ br.T, lr * hi + li * hr + u @ bi.T
+        y = torch.relu(hr @ Wa.T + ca) @ Wb.T + cb
+        loss = loss + ((y - xt[:, k]) ** 2).sum()
+    loss = loss / (Bn * 3 * (T1 - 1))
+    loss.backward()
+    G = out["grads"]
+    assert np.isclose(out["loss"], float(loss.detach()), rtol=1e-12)
+    assert np.allclose(G["lam"], lr.grad.numpy() + 1j * li.grad.numpy(), rtol=1e-9, atol=1e-13)
+    assert np.allclose(G["Bc"], br.grad.numpy() + 1j * bi.grad.numpy(), rtol=1e-9, atol=1e-13)
+    for k, v in [("Wa", Wa), ("ca", ca), ("Wb", Wb), ("cb", cb)]:
+        assert np.allclose(G[k], v.grad.numpy(), rtol=1e-9, atol=1e-13), k

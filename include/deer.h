@@ -1,0 +1,187 @@
+/*
+ * deer.h - C ABI of libdeer: the GTF-DEER hot path on AMD Instinct MI355X (gfx950).
+ *
+ * GTF-DEER (Hess, Goetz, Durstewitz, "Parallel-in-Time Training of Recurrent
+ * Neural Networks for Dynamical Systems Reconstruction") solves the forced
+ * recurrence z_t = F(z~_{t-1}) for all t at once by Newton's method: every
+ * iteration evaluates the residual and the forced Jacobians at all steps and
+ * solves the linear recursion Delta_t = J~_t Delta_{t-1} - r_t with a parallel
+ * associative scan (section "DSR from long sequences", eqs. GTF_residual and
+ * GTF_DEER_update; Alg. GTF-DEER).  Gradients come from the implicit function
+ * theorem: one scan of the same kind, run backwards with transposed Jacobians
+ * (gradients appendix, eqs. adjoint_eq and backward_recursion).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All arrays are float32, row-major, contiguous, batch-major and live in
+ *    device memory, except where an argument is marked "host".
+ *  - x    [B, T+1, N]  observations x_0..x_T (N = forcing.n_forced).
+ *  - z    [B, T, M]    states z_1..z_T; z[b, k] is z_{k+1}.
+ *  - z0   [B, M]       initial state; NULL means z_0 = B^+ x_0 = [x_0; 0].
+ *  - Observation model B = [I_N 0] (identity read-out of the first N latents,
+ *    model-setup appendix), so P_alpha = I - alpha B^+ B = diag(1 - a) with
+ *    a_i = alpha for i < N and a_i = 0 otherwise (eq. error_forcing).
+ *  - Step k+1 (array index k) reads the forced state
+ *        z~_k = (1 - a) * z_k + a * [x_k; 0]   for k >= 1,   z~_0 = z_0,
+ *    computed in float32 as fl(fl(p*z) + fl(a*zbar)), p = fl(1 - a), no fused
+ *    multiply-add, so that the ReLU decision below is reproducible bit for bit.
+ *  - masks [B, T, W] uint32, W = ceil(H/32): bit j of step k is (u_j > 0) with
+ *    u = z~_k (vanilla PLRNN, H = M) or u = h2 + W2 z~_k (shallow PLRNN, H = L;
+ *    u accumulated left to right in j from h2 in float32, one rounding after
+ *    every multiply and every add).  phi'(0) = 0.
+ *  - Every call runs on `stream` (a hipStream_t; NULL = the null stream).
+ *    Buffers are owned by the caller; the library never allocates or frees
+ *    device memory.  Scratch space comes from `ws` (device, `ws_bytes` bytes,
+ *    at least deer_workspace_bytes(...); 256-byte aligned).
+ *  - Errors are returned as a status code (never thrown across the ABI);
+ *    argument errors are detected before any device work is queued.
+ *    deer_last_error() gives a thread-local message for the last failure.
+ *  - The library keeps no mutable global state; calls on different streams
+ *    with different workspaces may run concurrently.  Calls that share a
+ *    workspace must be serialised by the caller.
+ */
+#ifndef DEER_H
+#define DEER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------------------- */
+enum {
+    DEER_OK = 0,
+    DEER_ERR_INVALID_ARG = 1,     /* null pointer, B/T/M out of range, alpha not in [0,1], ... */
+    DEER_ERR_NOT_CONVERGED = 2,   /* max_iter reached; z holds the last iterate */
+    DEER_ERR_NONFINITE = 3,       /* a Newton update produced NaN or Inf */
+    DEER_ERR_HIP = 4,             /* a HIP runtime call failed */
+    DEER_ERR_WORKSPACE = 5        /* ws too small or misaligned */
+};
+
+/* ---- models ------------------------------------------------------------------------ */
+enum {
+    DEER_PLRNN = 0,    /* z' = diag(A) z~ + W relu(z~) + h                       (W [M,M])   */
+    DEER_SHPLRNN = 1,  /* z' = diag(A) z~ + W relu(W2 z~ + h2) + h     (W [M,L], W2 [L,M])  */
+    DEER_DIAG_SSM = 2  /* h' = lambda * h + Bc u (complex diagonal, eq. shplrnn_ssm)        */
+};
+
+/* Parameters (device pointers).  The PLRNN kinds are eq. shplrnn_nonlinear with
+ * V = I, b = 0 (vanilla) or V = W2, b = h2 (shallow); no external inputs.
+ * DEER_DIAG_SSM: A = lambda [M][2] (re, im), W = Bc [M, L][2] with L the input
+ * dimension (inputs u_t = x_{t-1}), other pointers unused. */
+typedef struct {
+    int kind;
+    int M;              /* latent dimension: 1..64 for the PLRNN kinds, >= 1 for DIAG_SSM */
+    int L;              /* shallow: hidden width (1..1024); DIAG_SSM: input dimension       */
+    const float *A;
+    const float *W;
+    const float *W2;
+    const float *h;     /* may be NULL (zero) */
+    const float *h2;    /* may be NULL (zero) */
+} deer_model;
+
+typedef struct {
+    float alpha;        /* GTF forcing strength in [0, 1] (eq. GTF)                          */
+    int n_forced;       /* N: the first N latents are observed and forced, 0 <= N <= M      */
+} deer_forcing;
+
+enum { DEER_INIT_TEACHER = 0, DEER_INIT_ZERO = 1, DEER_INIT_USER = 2 };
+
+typedef struct {
+    float tol;          /* stop a sequence once max_{t,m} |Delta z| < tol (absolute)        */
+    int max_iter;       /* cap on Newton updates per sequence (500 if <= 0)                 */
+    int fixed_iters;    /* > 0: run exactly this many updates, no convergence test/sync     */
+    int init;           /* DEER_INIT_*: z^(0) = [x_{1:T}; 0], zeros, or z as passed in       */
+} deer_solve_opts;
+
+/* Per-parameter gradient outputs (device, float32, NULL to skip).
+ * PLRNN: A [M], W [M,M], h [M].  SHPLRNN: A [M], W [M,L] (=W1), W2 [L,M], h [M] (=h1),
+ * h2 [L].  DIAG_SSM: A = dlambda [M][2], W = dBc [M,L][2] (d/dRe + i d/dIm). */
+typedef struct {
+    float *A;
+    float *W;
+    float *W2;
+    float *h;
+    float *h2;
+} deer_grads;
+
+enum { DEER_OP_SOLVE = 0, DEER_OP_ADJOINT = 1 };
+enum { DEER_SCAN_DENSE = 0, DEER_SCAN_DIAG_C64 = 1 };
+
+/* Bytes of workspace `op` (DEER_OP_SOLVE or DEER_OP_ADJOINT) needs for this model and
+ * size.  Returns 0 for invalid arguments. */
+size_t deer_workspace_bytes(const deer_model *model, int B, int T, int op);
+
+/* GTF-DEER forward solve (Alg. GTF-DEER, Newton loop; eqs. GTF_residual, GTF_DEER_update).
+ *   x, z0        inputs as above; z0 may be NULL.
+ *   z            [B,T,M] out (in as well when opts->init == DEER_INIT_USER).  For
+ *                DEER_DIAG_SSM, z is h [B,T,M][2] (complex) and the call is the single
+ *                linear scan h_t = lambda h_{t-1} + Bc x_{t-1}, h_0 = 0 (Alg. LSSM).
+ *   masks        [B,T,W] out or NULL: activation masks at the returned z.
+ *   iters        host [B] out or NULL: updates applied to each sequence, counting the
+ *                verifying one (a sequence converged after k updates reports k).
+ *   final_norm   host [B] out or NULL: max |Delta z| of each sequence's last update.
+ * Each Newton update is applied before the test; a sequence whose update is below tol
+ * is frozen while the others continue.  With fixed_iters == 0 the call synchronises
+ * `stream` once per iteration (one device-to-host copy of B+2 words); with
+ * fixed_iters > 0 it synchronises once at the end (only if iters/final_norm given).
+ * Returns DEER_OK, DEER_ERR_NOT_CONVERGED (z = last iterate), DEER_ERR_NONFINITE or an
+ * argument / HIP / workspace error. */
+int deer_solve(const deer_model *model, const deer_forcing *forcing, const deer_solve_opts *opts,
+               int B, int T, const float *x, const float *z0, float *z, uint32_t *masks,
+               int32_t *iters, float *final_norm, void *ws, size_t ws_bytes, void *stream);
+
+/* Adjoint of the forced recurrence at a (converged) trajectory z (gradients appendix):
+ *   lam_T = g_T,  lam_{t-1} = J~_t^T lam_t + g_{t-1},   J~_t = J_F(z~_{t-1}) P_alpha,
+ * i.e. lam = dL/dz (the paper's v with the opposite sign), and the parameter gradients
+ *   dL/dtheta = sum_{b,t} lam_t^T dF(z~_{t-1})/dtheta.
+ *   g     [B,T,M] or NULL.  NULL: the MSE seed g_t = 2/(B N T) [z_t[:N] - x_t; 0] of the
+ *         batch-mean loss (eq. mse_loss_series).  DIAG_SSM: g is required, complex
+ *         [B,T,M][2] = dL/dRe h + i dL/dIm h, the recursion uses conj(lambda), and z is
+ *         the forward h.
+ *   lam   [B,T,M] out (DIAG_SSM: [B,T,M][2]) or NULL.
+ *   grads per-parameter outputs or NULL (sums over all (b, t), reduced in float64).
+ * Fully asynchronous on `stream`. */
+int deer_adjoint(const deer_model *model, const deer_forcing *forcing, int B, int T,
+                 const float *x, const float *z0, const float *z, const float *g,
+                 float *lam, const deer_grads *grads, void *ws, size_t ws_bytes, void *stream);
+
+/* Residual and forced Jacobians of a PLRNN kind at trajectory z (eq. GTF_residual; the
+ * Jacobian of F in the model-setup appendix; eq. error_forcing_decomp):
+ *   F     [B,T,M] out or NULL: F(z~_{t-1}).
+ *   r     [B,T,M] out or NULL: z_t - F(z~_{t-1}).
+ *   J     [B,T,M,M] out or NULL: J~_t = J_F(z~_{t-1}) P_alpha, row-major per step.
+ *   masks [B,T,W] out or NULL.
+ * No workspace; fully asynchronous. */
+int plrnn_jacobian(const deer_model *model, const deer_forcing *forcing, int B, int T,
+                   const float *x, const float *z0, const float *z, float *F, float *r, float *J,
+                   uint32_t *masks, void *stream);
+
+/* The bare associative scan over affine pairs (scheduled-sampling appendix: the pair
+ * (A_t, b_t) and its composition), batched over B independent sequences of length T.
+ *   DEER_SCAN_DENSE:    J [B,T,M,M], b [B,T,M], M <= 64.
+ *        reverse == 0:  y_t = J_t y_{t-1} + b_t, y_0 = 0        (J_1 is not read)
+ *        reverse != 0:  y_T = b_T, y_{t-1} = J_t^T y_t + b_{t-1}  (J_1 is not read)
+ *   DEER_SCAN_DIAG_C64: J = lambda [M][2], b [B,T,M][2] complex.
+ *        reverse == 0:  y_t = lambda y_{t-1} + b_t, y_0 = 0
+ *        reverse != 0:  y_T = b_T, y_{t-1} = conj(lambda) y_t + b_{t-1}
+ *   y     out, same layout as b (may not alias b).
+ * Fully asynchronous. */
+int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, const float *b, float *y,
+              void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes deer_scan needs. */
+size_t deer_scan_workspace_bytes(int layout, int B, int T, int M);
+
+/* Static description of a status code; never NULL. */
+const char *deer_status_string(int status);
+
+/* Thread-local message describing the last failing call on this thread ("" if none). */
+const char *deer_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DEER_H */

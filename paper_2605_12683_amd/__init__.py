@@ -1,0 +1,204 @@
+"""GTF-DEER hot path on AMD Instinct MI355X: Python binding of libdeer.
+
+The functions below carry the names of the C entry points (include/deer.h) and take
+torch tensors that already live on the GPU; they only marshal arguments, allocate the
+outputs and the workspace with torch, and call the library on torch's current stream.
+
+Model dictionaries use the paper's names:
+  vanilla PLRNN  {"kind": "plrnn",   "A": [M], "W": [M,M], "h": [M]}
+  shallow PLRNN  {"kind": "shplrnn", "A": [M], "W1": [M,L], "W2": [L,M], "h1": [M], "h2": [L]}
+  diagonal SSM   {"kind": "diag_ssm", "lam": complex64 [M], "Bc": complex64 [M,K]}
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _binding as _b
+from ._binding import DeerError, load  # noqa: F401
+
+__all__ = ["deer_solve", "deer_adjoint", "plrnn_jacobian", "deer_scan", "deer_workspace_bytes",
+           "deer_scan_workspace_bytes", "deer_status_string", "DeerError", "load"]
+
+_KINDS = {"plrnn": _b.DEER_PLRNN, "shplrnn": _b.DEER_SHPLRNN, "diag_ssm": _b.DEER_DIAG_SSM}
+_INITS = {"teacher": _b.DEER_INIT_TEACHER, "zero": _b.DEER_INIT_ZERO, "user": _b.DEER_INIT_USER}
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t, dtype=torch.float32):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        t = torch.as_tensor(t)
+    if t.is_complex():
+        t = torch.view_as_real(t.to(torch.complex64).contiguous())
+    t = t.to(device="cuda", dtype=dtype).contiguous()
+    return t
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+class _Model:
+    """Device copies of the parameters plus the C struct that points at them."""
+
+    def __init__(self, model: dict):
+        kind = model["kind"]
+        self.kind = kind
+        if kind == "plrnn":
+            self.t = {k: _dev(model[k]) for k in ("A", "W")}
+            self.t["h"] = _dev(model.get("h"))
+            M = self.t["A"].shape[0]
+            self.c = _b.deer_model(_b.DEER_PLRNN, M, 0, _ptr(self.t["A"]), _ptr(self.t["W"]), None,
+                                   _ptr(self.t["h"]), None)
+        elif kind == "shplrnn":
+            self.t = {k: _dev(model[k]) for k in ("A", "W1", "W2")}
+            self.t["h1"] = _dev(model.get("h1"))
+            self.t["h2"] = _dev(model.get("h2"))
+            M, L = self.t["W1"].shape
+            self.c = _b.deer_model(_b.DEER_SHPLRNN, M, L, _ptr(self.t["A"]), _ptr(self.t["W1"]), _ptr(self.t["W2"]),
+                                   _ptr(self.t["h1"]), _ptr(self.t["h2"]))
+        elif kind == "diag_ssm":
+            self.t = {"lam": _dev(model["lam"]), "Bc": _dev(model["Bc"])}
+            M, K = self.t["Bc"].shape[:2]
+            self.c = _b.deer_model(_b.DEER_DIAG_SSM, M, K, _ptr(self.t["lam"]), _ptr(self.t["Bc"]), None, None, None)
+        else:
+            raise ValueError(kind)
+        self.M = self.c.M
+        self.L = self.c.L
+
+
+def _model(model):
+    return model if isinstance(model, _Model) else _Model(model)
+
+
+def deer_status_string(status: int) -> str:
+    return load().deer_status_string(status).decode()
+
+
+def deer_workspace_bytes(model, B: int, T: int, op: int) -> int:
+    m = _model(model)
+    return int(load().deer_workspace_bytes(ctypes.byref(m.c), B, T, op))
+
+
+def deer_scan_workspace_bytes(layout: int, B: int, T: int, M: int) -> int:
+    return int(load().deer_scan_workspace_bytes(layout, B, T, M))
+
+
+def _workspace(nbytes: int):
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+
+
+def deer_solve(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1e-5, max_iter: int = 500,
+               fixed_iters: int = 0, init: str = "teacher", z=None, want_masks: bool = False, ws=None,
+               check: bool = True) -> dict:
+    """GTF-DEER forward solve.  Returns dict(z, masks, iters, norms, status)."""
+    lib = load()
+    m = _model(model)
+    x = _dev(x)
+    B, T1, _ = x.shape
+    T = T1 - 1
+    if m.kind == "diag_ssm":
+        out = torch.empty(B, T, m.M, 2, device="cuda") if z is None else z
+    else:
+        out = torch.empty(B, T, m.M, device="cuda") if z is None else z
+    if init == "user" and z is None:
+        raise ValueError("init='user' needs z")
+    masks = None
+    if want_masks:
+        H = m.M if m.kind == "plrnn" else m.L
+        masks = torch.empty(B, T, (H + 31) // 32, dtype=torch.int32, device="cuda")
+    if ws is None:
+        ws = _workspace(lib.deer_workspace_bytes(ctypes.byref(m.c), B, T, _b.DEER_OP_SOLVE))
+    iters = (ctypes.c_int32 * B)()
+    norms = (ctypes.c_float * B)()
+    f = _b.deer_forcing(float(alpha), int(n_forced))
+    o = _b.deer_solve_opts(float(tol), int(max_iter), int(fixed_iters), _INITS[init])
+    z0d = _dev(z0)
+    st = lib.deer_solve(ctypes.byref(m.c), ctypes.byref(f), ctypes.byref(o), B, T, _ptr(x), _ptr(z0d), _ptr(out),
+                        _ptr(masks), iters, norms, _ptr(ws), ws.numel(), _stream())
+    if check:
+        _check_solve = (_b.DEER_OK, _b.DEER_ERR_NOT_CONVERGED, _b.DEER_ERR_NONFINITE)
+        _b._check(st, "deer_solve", allow=_check_solve)
+    return {"z": out, "masks": masks, "iters": list(iters), "norms": list(norms), "status": st}
+
+
+def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, want_lam: bool = True,
+                 want_grads: bool = True, ws=None) -> dict:
+    """Adjoint scan lam = dL/dz and parameter gradients at trajectory z."""
+    lib = load()
+    m = _model(model)
+    x = _dev(x)
+    B, T1, _ = x.shape
+    T = T1 - 1
+    z = _dev(z)
+    g = _dev(g)
+    shape = (B, T, m.M, 2) if m.kind == "diag_ssm" else (B, T, m.M)
+    lam = torch.empty(shape, device="cuda") if (want_lam or m.kind == "diag_ssm") else None
+    grads = {}
+    gs = _b.deer_grads()
+    if want_grads:
+        if m.kind == "plrnn":
+            grads = {"A": torch.empty(m.M, device="cuda"), "W": torch.empty(m.M, m.M, device="cuda"),
+                     "h": torch.empty(m.M, device="cuda")}
+            gs = _b.deer_grads(_ptr(grads["A"]), _ptr(grads["W"]), None, _ptr(grads["h"]), None)
+        elif m.kind == "shplrnn":
+            grads = {"A": torch.empty(m.M, device="cuda"), "W1": torch.empty(m.M, m.L, device="cuda"),
+                     "W2": torch.empty(m.L, m.M, device="cuda"), "h1": torch.empty(m.M, device="cuda"),
+                     "h2": torch.empty(m.L, device="cuda")}
+            gs = _b.deer_grads(_ptr(grads["A"]), _ptr(grads["W1"]), _ptr(grads["W2"]), _ptr(grads["h1"]),
+                               _ptr(grads["h2"]))
+        else:
+            grads = {"lam": torch.empty(m.M, 2, device="cuda"), "Bc": torch.empty(m.M, m.L, 2, device="cuda")}
+            gs = _b.deer_grads(_ptr(grads["lam"]), _ptr(grads["Bc"]), None, None, None)
+    if ws is None:
+        ws = _workspace(lib.deer_workspace_bytes(ctypes.byref(m.c), B, T, _b.DEER_OP_ADJOINT))
+    f = _b.deer_forcing(float(alpha), int(n_forced))
+    z0d = _dev(z0)
+    st = lib.deer_adjoint(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(g), _ptr(lam),
+                          ctypes.byref(gs), _ptr(ws), ws.numel(), _stream())
+    _b._check(st, "deer_adjoint")
+    return {"lam": lam, "grads": grads}
+
+
+def plrnn_jacobian(model, x, z, alpha: float, n_forced: int, *, z0=None, want=("F", "r", "masks"),
+                   dense_J: bool = False) -> dict:
+    """F, r, masks (and optionally the dense forced Jacobians) at trajectory z."""
+    lib = load()
+    m = _model(model)
+    x = _dev(x)
+    z = _dev(z)
+    B, T, M = z.shape
+    H = m.M if m.kind == "plrnn" else m.L
+    out = {}
+    F = torch.empty(B, T, M, device="cuda") if "F" in want else None
+    r = torch.empty(B, T, M, device="cuda") if "r" in want else None
+    J = torch.empty(B, T, M, M, device="cuda") if dense_J else None
+    masks = torch.empty(B, T, (H + 31) // 32, dtype=torch.int32, device="cuda") if "masks" in want else None
+    f = _b.deer_forcing(float(alpha), int(n_forced))
+    z0d = _dev(z0)
+    st = lib.plrnn_jacobian(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(F), _ptr(r),
+                            _ptr(J), _ptr(masks), _stream())
+    _b._check(st, "plrnn_jacobian")
+    out.update({"F": F, "r": r, "J": J, "masks": masks})
+    return out
+
+
+def deer_scan(layout: int, J, b, reverse: bool = False, ws=None):
+    """Bare affine scan (DEER_SCAN_DENSE: J [B,T,M,M]; DEER_SCAN_DIAG_C64: lambda [M] complex)."""
+    lib = load()
+    J = _dev(J)
+    b = _dev(b)
+    B, T, M = b.shape[:3]
+    y = torch.empty_like(b)
+    if ws is None:
+        ws = _workspace(lib.deer_scan_workspace_bytes(layout, B, T, M))
+    st = lib.deer_scan(layout, 1 if reverse else 0, B, T, M, _ptr(J), _ptr(b), _ptr(y), _ptr(ws), ws.numel(),
+                       _stream())
+    _b._check(st, "deer_scan")
+    return y

@@ -1,0 +1,94 @@
+"""ctypes binding of libdeer (the C ABI in include/deer.h).
+
+Argument marshalling only: every step of the GTF-DEER path runs in the HIP kernels of
+libdeer.so.  PyTorch provides device memory and the stream.  There is no fallback: if the
+library is missing, loading fails with an error.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdeer.so")
+
+DEER_OK, DEER_ERR_INVALID_ARG, DEER_ERR_NOT_CONVERGED, DEER_ERR_NONFINITE, DEER_ERR_HIP, DEER_ERR_WORKSPACE = range(6)
+DEER_PLRNN, DEER_SHPLRNN, DEER_DIAG_SSM = 0, 1, 2
+DEER_INIT_TEACHER, DEER_INIT_ZERO, DEER_INIT_USER = 0, 1, 2
+DEER_OP_SOLVE, DEER_OP_ADJOINT = 0, 1
+DEER_SCAN_DENSE, DEER_SCAN_DIAG_C64 = 0, 1
+
+EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "plrnn_jacobian", "deer_scan",
+            "deer_scan_workspace_bytes", "deer_status_string", "deer_last_error"]
+
+_fp = ctypes.c_void_p
+
+
+class deer_model(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("M", ctypes.c_int), ("L", ctypes.c_int),
+                ("A", _fp), ("W", _fp), ("W2", _fp), ("h", _fp), ("h2", _fp)]
+
+
+class deer_forcing(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_float), ("n_forced", ctypes.c_int)]
+
+
+class deer_solve_opts(ctypes.Structure):
+    _fields_ = [("tol", ctypes.c_float), ("max_iter", ctypes.c_int), ("fixed_iters", ctypes.c_int),
+                ("init", ctypes.c_int)]
+
+
+class deer_grads(ctypes.Structure):
+    _fields_ = [("A", _fp), ("W", _fp), ("W2", _fp), ("h", _fp), ("h2", _fp)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libdeer.so and declare its signatures (raises if the library is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2605_12683_amd.build` "
+                           "(there is no non-HIP fallback)")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    sz, i32, vp = ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p
+    lib.deer_workspace_bytes.argtypes = [P(deer_model), i32, i32, i32]
+    lib.deer_workspace_bytes.restype = sz
+    lib.deer_scan_workspace_bytes.argtypes = [i32, i32, i32, i32]
+    lib.deer_scan_workspace_bytes.restype = sz
+    lib.deer_solve.argtypes = [P(deer_model), P(deer_forcing), P(deer_solve_opts), i32, i32, vp, vp, vp, vp,
+                               P(ctypes.c_int32), P(ctypes.c_float), vp, sz, vp]
+    lib.deer_solve.restype = i32
+    lib.deer_adjoint.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, vp, P(deer_grads), vp, sz,
+                                 vp]
+    lib.deer_adjoint.restype = i32
+    lib.plrnn_jacobian.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.plrnn_jacobian.restype = i32
+    lib.deer_scan.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]
+    lib.deer_scan.restype = i32
+    lib.deer_status_string.argtypes = [i32]
+    lib.deer_status_string.restype = ctypes.c_char_p
+    lib.deer_last_error.argtypes = []
+    lib.deer_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+class DeerError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        lib = load()
+        msg = lib.deer_last_error().decode() or lib.deer_status_string(status).decode()
+        super().__init__(f"{where}: {lib.deer_status_string(status).decode()} ({msg})")
+        self.status = status
+
+
+def _check(status: int, where: str, allow=(DEER_OK,)):
+    if status not in allow:
+        raise DeerError(status, where)
+    return status

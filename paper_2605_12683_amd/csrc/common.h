@@ -1,0 +1,73 @@
+// Internal helpers shared by the libdeer translation units (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "../../include/deer.h"
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+namespace deer {
+
+// ---- host-side error plumbing --------------------------------------------------------
+void set_error(const char *fmt, ...);
+int hip_fail(hipError_t e, const char *what);
+
+#define DEER_HIP(call)                                                 \
+    do {                                                               \
+        hipError_t _e = (call);                                        \
+        if (_e != hipSuccess) return ::deer::hip_fail(_e, #call);      \
+    } while (0)
+
+#define DEER_LAUNCH_CHECK(what)                                        \
+    do {                                                               \
+        hipError_t _e = hipGetLastError();                             \
+        if (_e != hipSuccess) return ::deer::hip_fail(_e, what);       \
+    } while (0)
+
+// ---- device helpers ---------------------------------------------------------------------
+
+// 16x16x4 fp32 MFMA: acc[16x16] += A[16x4] * B[4x16].  Lane l = 16*g + c holds
+// A[c][g], B[g][c] and acc[4*g + r][c] in element r of the returned vector.
+__device__ __forceinline__ v4f mfma16x16x4(float a, float b, v4f acc) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+}
+
+// all-ones if bit `sh` of w is set, else zero (sign-extended one-bit field)
+__device__ __forceinline__ float select_bit(uint32_t w, int sh, float v) {
+    int m = __builtin_amdgcn_sbfe((int)w, sh, 1);
+    return __int_as_float(__float_as_int(v) & m);
+}
+
+// |v| as ordered bits: NaN (any sign) compares above +Inf, so an unsigned max keeps NaN.
+__device__ __forceinline__ uint32_t abs_bits(float v) {
+    return (uint32_t)__float_as_int(v) & 0x7fffffffu;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    for (int off = 32; off > 0; off >>= 1) {
+        uint32_t o = (uint32_t)__shfl_xor((int)v, off, 64);
+        v = v > o ? v : o;
+    }
+    return v;
+}
+
+// forced input of step s (array index) for latent i:
+//   s == 0: z0 (or [x_0; 0] when z0 is null);  s >= 1: fl(fl(p*z_{s-1}) + fl(a*zbar_s))
+__device__ __forceinline__ float forced_state(const float *__restrict__ x, const float *__restrict__ z0,
+                                              const float *__restrict__ z, int b, int s, int i, int T, int M,
+                                              int N, float alpha) {
+    if (s == 0) {
+        if (z0) return z0[(size_t)b * M + i];
+        return i < N ? x[(size_t)b * (T + 1) * N + i] : 0.0f;
+    }
+    float zp = z[((size_t)b * T + (s - 1)) * M + i];
+    if (i >= N) return zp;
+    float zb = x[((size_t)b * (T + 1) + s) * N + i];
+    float p = __fsub_rn(1.0f, alpha);
+    return __fadd_rn(__fmul_rn(p, zp), __fmul_rn(alpha, zb));
+}
+
+}  // namespace deer

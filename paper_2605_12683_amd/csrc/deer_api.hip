@@ -1,0 +1,396 @@
+// C ABI of libdeer: argument validation, workspace carving and the host-side Newton loop
+// of GTF-DEER (Alg. GTF-DEER).  All device work is queued on the caller's stream.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "common.h"
+#include "launch.h"
+
+namespace deer {
+
+static thread_local char g_err[512] = "";
+
+void set_error(const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    set_error("%s failed: %s", what, hipGetErrorString(e));
+    return DEER_ERR_HIP;
+}
+
+// ---- small utility kernels -------------------------------------------------------------
+__global__ void k_fill_teacher(int B, int T, int M, int N, const float *__restrict__ x, float *__restrict__ z) {
+    const size_t n = (size_t)B * T * M;
+    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n; e += (size_t)gridDim.x * blockDim.x) {
+        const int i = (int)(e % M);
+        const size_t bt = e / M;
+        const int b = (int)(bt / T), s = (int)(bt % T);
+        z[e] = i < N ? x[((size_t)b * (T + 1) + s + 1) * N + i] : 0.f;
+    }
+}
+__global__ void k_fill_i32(int *p, int n, int v) {
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e < n) p[e] = v;
+}
+__global__ void k_fill_f32(float *p, size_t n, float v) {
+    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n; e += (size_t)gridDim.x * blockDim.x) p[e] = v;
+}
+
+int launch_fill_teacher(int B, int T, int M, int N, const float *x, float *z, hipStream_t st) {
+    const size_t n = (size_t)B * T * M;
+    const int grid = (int)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
+    hipLaunchKernelGGL(k_fill_teacher, dim3(grid), dim3(256), 0, st, B, T, M, N, x, z);
+    DEER_LAUNCH_CHECK("k_fill_teacher");
+    return DEER_OK;
+}
+int launch_fill_i32(int *p, int n, int v, hipStream_t st) {
+    hipLaunchKernelGGL(k_fill_i32, dim3((n + 255) / 256), dim3(256), 0, st, p, n, v);
+    DEER_LAUNCH_CHECK("k_fill_i32");
+    return DEER_OK;
+}
+int launch_fill_f32(float *p, size_t n, float v, hipStream_t st) {
+    const int grid = (int)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
+    hipLaunchKernelGGL(k_fill_f32, dim3(grid), dim3(256), 0, st, p, n, v);
+    DEER_LAUNCH_CHECK("k_fill_f32");
+    return DEER_OK;
+}
+
+// ---- workspace carving ---------------------------------------------------------------------
+struct Carver {
+    char *base;
+    size_t off = 0;
+    explicit Carver(void *b) : base((char *)b) {}
+    template <class Tp>
+    Tp *take(size_t count) {
+        Tp *p = base ? (Tp *)(base + off) : nullptr;
+        off += (count * sizeof(Tp) + 255) & ~(size_t)255;
+        return p;
+    }
+};
+
+static int chunk_override() {
+    const char *e = getenv("DEER_CHUNK");
+    return e ? atoi(e) : 0;
+}
+
+// Chunk length of the dense scans: enough chains to fill the machine (about 2048 waves),
+// at most 128 chunks per sequence so that the serial carry pass stays short.
+static int choose_chunk(int B, int T, int MP) {
+    const int ov = chunk_override();
+    if (ov > 0) return ov < T ? ov : T;
+    const long total = (long)B * T;
+    const long target_chains = 2048L * (64 / MP);
+    long C = (total + target_chains - 1) / target_chains;
+    if (C < 16) C = 16;
+    const long minC = (T + 127) / 128;
+    if (C < minC) C = minC;
+    if (C > T) C = T;
+    return (int)C;
+}
+
+struct PlrnnWs {
+    float *r;
+    uint32_t *masks;
+    float *P, *v, *carry;
+    uint32_t *norm_bits;
+    int *active;
+    float *gpart;
+    int C, ncs, MP;
+};
+
+static PlrnnWs carve_plrnn(void *ws, int B, int T, int M, int op, size_t *bytes) {
+    PlrnnWs w{};
+    w.MP = padded_dim(M);
+    w.C = choose_chunk(B, T, w.MP);
+    w.ncs = (T + w.C - 1) / w.C;
+    const size_t nch = (size_t)B * w.ncs;
+    const int MW = (M + 31) / 32;
+    Carver c(ws);
+    w.masks = c.take<uint32_t>((size_t)B * T * MW);
+    w.P = c.take<float>(nch * w.MP * w.MP);
+    w.v = c.take<float>(nch * w.MP);
+    w.carry = c.take<float>(nch * w.MP);
+    w.norm_bits = c.take<uint32_t>(B);
+    w.active = c.take<int>(B);
+    if (op == DEER_OP_SOLVE) {
+        w.r = c.take<float>((size_t)B * T * M);
+    } else {
+        w.gpart = c.take<float>(nch * w.MP * (w.MP + 2));
+    }
+    *bytes = c.off;
+    return w;
+}
+
+static int check_common(const deer_model *m, const deer_forcing *f, int B, int T) {
+    if (!m || !f) { set_error("model/forcing pointer is NULL"); return DEER_ERR_INVALID_ARG; }
+    if (B <= 0 || T <= 0) { set_error("B and T must be positive (B=%d, T=%d)", B, T); return DEER_ERR_INVALID_ARG; }
+    if (!(f->alpha >= 0.0f && f->alpha <= 1.0f)) { set_error("alpha must lie in [0, 1]"); return DEER_ERR_INVALID_ARG; }
+    if (m->M <= 0) { set_error("M must be positive"); return DEER_ERR_INVALID_ARG; }
+    if (m->kind == DEER_PLRNN || m->kind == DEER_SHPLRNN) {
+        if (m->M > 64) { set_error("M=%d unsupported (dense scans support M <= 64)", m->M); return DEER_ERR_INVALID_ARG; }
+        if (f->n_forced < 0 || f->n_forced > m->M) { set_error("n_forced must lie in [0, M]"); return DEER_ERR_INVALID_ARG; }
+        if (!m->A || !m->W) { set_error("model parameters A and W are required"); return DEER_ERR_INVALID_ARG; }
+        if (m->kind == DEER_SHPLRNN) {
+            if (m->L <= 0 || m->L > 1024 || !m->W2) { set_error("shallow PLRNN needs W2 and 1 <= L <= 1024"); return DEER_ERR_INVALID_ARG; }
+        }
+    } else if (m->kind == DEER_DIAG_SSM) {
+        if (!m->A || !m->W) { set_error("DIAG_SSM needs lambda (A) and Bc (W)"); return DEER_ERR_INVALID_ARG; }
+        if (m->L <= 0 || m->L > 4) { set_error("DIAG_SSM input dimension L must lie in [1, 4]"); return DEER_ERR_INVALID_ARG; }
+    } else {
+        set_error("unknown model kind %d", m->kind);
+        return DEER_ERR_INVALID_ARG;
+    }
+    if ((long)B * (long)T > (1L << 31) / 1) { set_error("B*T too large"); return DEER_ERR_INVALID_ARG; }
+    return DEER_OK;
+}
+
+static int check_ws(void *ws, size_t have, size_t need) {
+    if (need == 0) return DEER_OK;
+    if (!ws || have < need) {
+        set_error("workspace too small: need %zu bytes, have %zu", need, ws ? have : (size_t)0);
+        return DEER_ERR_WORKSPACE;
+    }
+    if (((uintptr_t)ws & 255u) != 0) { set_error("workspace must be 256-byte aligned"); return DEER_ERR_WORKSPACE; }
+    return DEER_OK;
+}
+
+static size_t diag_bytes(int B, int T, int M, int op) {
+    size_t a = diag_scan_ws_bytes(B, T, M);
+    if (op == DEER_OP_ADJOINT) {
+        size_t g = diag_grads_ws_bytes(B, T, M);
+        if (g > a) a = g;
+    }
+    return a;
+}
+
+}  // namespace deer
+
+using namespace deer;
+
+extern "C" {
+
+const char *deer_status_string(int s) {
+    switch (s) {
+        case DEER_OK: return "ok";
+        case DEER_ERR_INVALID_ARG: return "invalid argument";
+        case DEER_ERR_NOT_CONVERGED: return "Newton iteration did not converge within max_iter";
+        case DEER_ERR_NONFINITE: return "non-finite value in a Newton update";
+        case DEER_ERR_HIP: return "HIP runtime error";
+        case DEER_ERR_WORKSPACE: return "workspace too small or misaligned";
+        default: return "unknown status";
+    }
+}
+
+const char *deer_last_error(void) { return g_err; }
+
+size_t deer_workspace_bytes(const deer_model *m, int B, int T, int op) {
+    deer_forcing f{0.f, 0};
+    if (check_common(m, &f, B, T) != DEER_OK) return 0;
+    if (op != DEER_OP_SOLVE && op != DEER_OP_ADJOINT) return 0;
+    if (m->kind == DEER_DIAG_SSM) return diag_bytes(B, T, m->M, op);
+    if (m->kind == DEER_PLRNN) {
+        size_t bytes = 0;
+        carve_plrnn(nullptr, B, T, m->M, op, &bytes);
+        return bytes;
+    }
+    return 0;
+}
+
+size_t deer_scan_workspace_bytes(int layout, int B, int T, int M) {
+    if (B <= 0 || T <= 0 || M <= 0) return 0;
+    if (layout == DEER_SCAN_DIAG_C64) return diag_scan_ws_bytes(B, T, M);
+    return 0;
+}
+
+int plrnn_jacobian(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
+                   const float *z, float *F, float *r, float *J, uint32_t *masks, void *stream) {
+    set_error("");
+    int rc = check_common(m, f, B, T);
+    if (rc) return rc;
+    if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
+    hipStream_t st = (hipStream_t)stream;
+    if (m->kind == DEER_PLRNN) {
+        PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
+        return launch_resjac_plrnn(a, z, F, r, J, masks, nullptr, st);
+    }
+    set_error("plrnn_jacobian: model kind %d not supported", m->kind);
+    return DEER_ERR_INVALID_ARG;
+}
+
+static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
+                       const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
+                       void *ws, size_t ws_bytes, hipStream_t st) {
+    size_t need = 0;
+    carve_plrnn(nullptr, B, T, m->M, DEER_OP_SOLVE, &need);
+    int rc = check_ws(ws, ws_bytes, need);
+    if (rc) return rc;
+    PlrnnWs w = carve_plrnn(ws, B, T, m->M, DEER_OP_SOLVE, &need);
+    PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
+    const int fixed = o->fixed_iters > 0 ? o->fixed_iters : 0;
+    const int max_iter = o->max_iter > 0 ? o->max_iter : 500;
+    if (o->init == DEER_INIT_TEACHER) {
+        if ((rc = launch_fill_teacher(B, T, m->M, f->n_forced, x, z, st))) return rc;
+    } else if (o->init == DEER_INIT_ZERO) {
+        if ((rc = launch_fill_f32(z, (size_t)B * T * m->M, 0.f, st))) return rc;
+    }
+    if ((rc = launch_fill_i32(w.active, B, 1, st))) return rc;
+    std::vector<int> act(B, 1), it(B, 0);
+    std::vector<uint32_t> nb(B, 0);
+    std::vector<float> norm(B, NAN);
+    bool nonfinite = false;
+    const int *dact = fixed ? nullptr : w.active;
+    for (int k = 0;; ++k) {
+        if (fixed) {
+            if (k == fixed) break;
+        } else {
+            bool any = false;
+            for (int b = 0; b < B; ++b) any |= act[b] != 0;
+            if (!any || k == max_iter) break;
+        }
+        if ((rc = launch_resjac_plrnn(a, z, nullptr, w.r, nullptr, w.masks, dact, st))) return rc;
+        if ((rc = launch_chunk_product_plrnn(a, false, w.masks, w.r, nullptr, 0.f, w.P, w.v, dact, w.C, w.ncs, st)))
+            return rc;
+        if ((rc = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, w.norm_bits, B, w.ncs, st))) return rc;
+        if ((rc = launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, z, w.norm_bits, dact, w.C, w.ncs, st))) return rc;
+        if (fixed) continue;
+        DEER_HIP(hipMemcpyAsync(nb.data(), w.norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+        DEER_HIP(hipStreamSynchronize(st));
+        bool changed = false;
+        for (int b = 0; b < B; ++b) {
+            if (!act[b]) continue;
+            float e;
+            memcpy(&e, &nb[b], 4);
+            it[b] += 1;
+            norm[b] = e;
+            if (!isfinite(e)) {
+                nonfinite = true;
+                act[b] = 0;
+                changed = true;
+            } else if (e < o->tol) {
+                act[b] = 0;
+                changed = true;
+            }
+        }
+        if (changed) {
+            DEER_HIP(hipMemcpyAsync(w.active, act.data(), B * sizeof(int), hipMemcpyHostToDevice, st));
+            DEER_HIP(hipStreamSynchronize(st));
+        }
+    }
+    if (fixed && (iters || final_norm)) {
+        DEER_HIP(hipMemcpyAsync(nb.data(), w.norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+        DEER_HIP(hipStreamSynchronize(st));
+        for (int b = 0; b < B; ++b) {
+            memcpy(&norm[b], &nb[b], 4);
+            it[b] = fixed;
+            if (!isfinite(norm[b])) nonfinite = true;
+        }
+    }
+    if (masks) {
+        if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
+    }
+    if (iters) for (int b = 0; b < B; ++b) iters[b] = it[b];
+    if (final_norm) for (int b = 0; b < B; ++b) final_norm[b] = norm[b];
+    if (nonfinite) {
+        set_error("a Newton update produced a non-finite value");
+        return DEER_ERR_NONFINITE;
+    }
+    if (!fixed) {
+        for (int b = 0; b < B; ++b)
+            if (act[b]) {
+                set_error("sequence %d not converged after %d Newton updates (last max|dz| = %g)", b, it[b], norm[b]);
+                return DEER_ERR_NOT_CONVERGED;
+            }
+    }
+    return DEER_OK;
+}
+
+int deer_solve(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T, const float *x,
+               const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm, void *ws,
+               size_t ws_bytes, void *stream) {
+    set_error("");
+    int rc = check_common(m, f, B, T);
+    if (rc) return rc;
+    if (!o || !x || !z) { set_error("opts, x and z are required"); return DEER_ERR_INVALID_ARG; }
+    if (o->init < 0 || o->init > 2) { set_error("unknown init %d", o->init); return DEER_ERR_INVALID_ARG; }
+    if (!(o->tol >= 0.f) && o->fixed_iters <= 0) { set_error("tol must be >= 0"); return DEER_ERR_INVALID_ARG; }
+    hipStream_t st = (hipStream_t)stream;
+    if (m->kind == DEER_PLRNN)
+        return solve_plrnn(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
+    if (m->kind == DEER_DIAG_SSM) {
+        if ((rc = check_ws(ws, ws_bytes, diag_bytes(B, T, m->M, DEER_OP_SOLVE)))) return rc;
+        rc = launch_diag_scan(false, B, T, m->M, m->A, nullptr, m->W, m->L, x, z, ws, st);
+        if (rc) return rc;
+        if (iters) for (int b = 0; b < B; ++b) iters[b] = 1;
+        if (final_norm) for (int b = 0; b < B; ++b) final_norm[b] = 0.f;
+        return DEER_OK;
+    }
+    set_error("deer_solve: model kind %d not supported yet", m->kind);
+    return DEER_ERR_INVALID_ARG;
+}
+
+int deer_adjoint(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
+                 const float *z, const float *g, float *lam, const deer_grads *grads, void *ws, size_t ws_bytes,
+                 void *stream) {
+    set_error("");
+    int rc = check_common(m, f, B, T);
+    if (rc) return rc;
+    if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
+    hipStream_t st = (hipStream_t)stream;
+    if (m->kind == DEER_PLRNN) {
+        size_t need = 0;
+        carve_plrnn(nullptr, B, T, m->M, DEER_OP_ADJOINT, &need);
+        if ((rc = check_ws(ws, ws_bytes, need))) return rc;
+        PlrnnWs w = carve_plrnn(ws, B, T, m->M, DEER_OP_ADJOINT, &need);
+        PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
+        const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
+        if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, w.masks, nullptr, st))) return rc;
+        if ((rc = launch_chunk_product_plrnn(a, true, w.masks, g, z, scale, w.P, w.v, nullptr, w.C, w.ncs, st)))
+            return rc;
+        if ((rc = launch_carry(w.MP, true, w.P, w.v, w.carry, nullptr, nullptr, B, w.ncs, st))) return rc;
+        if ((rc = launch_fixup_rev_plrnn(a, w.masks, g, scale, z, w.carry, lam, w.gpart, w.C, w.ncs, st))) return rc;
+        if (grads && (grads->A || grads->W || grads->h)) {
+            if ((rc = launch_reduce_gpart(w.gpart, B * w.ncs, w.MP, m->M, grads->A, grads->W, grads->h, st))) return rc;
+        }
+        return DEER_OK;
+    }
+    if (m->kind == DEER_DIAG_SSM) {
+        if (!g) { set_error("DIAG_SSM adjoint needs the cotangent g"); return DEER_ERR_INVALID_ARG; }
+        if ((rc = check_ws(ws, ws_bytes, diag_bytes(B, T, m->M, DEER_OP_ADJOINT)))) return rc;
+        float *out = lam;
+        if (!out) { set_error("DIAG_SSM adjoint needs the lam output buffer"); return DEER_ERR_INVALID_ARG; }
+        if ((rc = launch_diag_scan(true, B, T, m->M, m->A, g, nullptr, m->L, nullptr, out, ws, st))) return rc;
+        if (grads && (grads->A || grads->W)) {
+            if ((rc = launch_diag_grads(B, T, m->M, m->L, out, z, x, grads->A, grads->W, ws, st))) return rc;
+        }
+        return DEER_OK;
+    }
+    set_error("deer_adjoint: model kind %d not supported yet", m->kind);
+    return DEER_ERR_INVALID_ARG;
+}
+
+int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, const float *b, float *y, void *ws,
+              size_t ws_bytes, void *stream) {
+    set_error("");
+    if (B <= 0 || T <= 0 || M <= 0) { set_error("B, T, M must be positive"); return DEER_ERR_INVALID_ARG; }
+    if (!J || !b || !y) { set_error("J, b and y are required"); return DEER_ERR_INVALID_ARG; }
+    if (b == y) { set_error("y may not alias b"); return DEER_ERR_INVALID_ARG; }
+    hipStream_t st = (hipStream_t)stream;
+    if (layout == DEER_SCAN_DIAG_C64) {
+        int rc = check_ws(ws, ws_bytes, diag_scan_ws_bytes(B, T, M));
+        if (rc) return rc;
+        return launch_diag_scan(reverse != 0, B, T, M, J, b, nullptr, 0, nullptr, y, ws, st);
+    }
+    set_error("deer_scan: layout %d not supported yet", layout);
+    return DEER_ERR_INVALID_ARG;
+}
+
+}  // extern "C"

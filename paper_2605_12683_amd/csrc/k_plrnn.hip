@@ -1,0 +1,578 @@
+// Vanilla PLRNN path of GTF-DEER on gfx950:
+//   z_t = diag(A) z~_{t-1} + W relu(z~_{t-1}) + h          (eq. shplrnn_nonlinear, V = I, b = 0)
+//   J~_t = (diag(A) + W diag(m_t)) P_alpha                  (Jacobian of F, eq. error_forcing_decomp)
+//
+// Kernels (one Newton iteration = resjac -> chunk products -> carries -> fix-up):
+//   k_resjac_plrnn     residual r_t, masks m_t (and optionally F, dense J~) at every step
+//   k_chunk_product    per chunk of C steps: P_c = J~_e ... J~_s on the matrix cores (fp32
+//                      MFMA) and v_c = the chunk's local solution from a zero carry (VALU)
+//   k_carry            carries across chunks, one wave per sequence
+//   k_fixup_fwd        Delta_t = J~_t Delta_{t-1} - r_t from the carry, z += Delta, max|Delta|
+//   k_fixup_rev        lam_{t-1} = J~_t^T lam_t + g_{t-1} from the carry, fused parameter-
+//                      gradient partial sums (gradients appendix)
+//
+// Padded dimension MP in {16, 32, 64} (the next one >= M); a wave holds NCH = 64/MP chains.
+#include "common.h"
+#include "launch.h"
+
+namespace deer {
+
+template <int MP>
+struct Geo {
+    static constexpr int NCH = 64 / MP;   // chains (or timesteps) per wave
+    static constexpr int NI = MP / 16;    // 16-row tiles
+    static constexpr int NS = MP / 4;     // k-steps of the 16x16x4 MFMA
+    static constexpr int MW = MP <= 32 ? 1 : 2;   // mask words per step
+};
+
+__device__ __forceinline__ float p_of(int i, int N, float alpha) { return i < N ? __fsub_rn(1.0f, alpha) : 1.0f; }
+
+__device__ __forceinline__ uint32_t mask_bit(const uint32_t *__restrict__ masks, size_t step, int MW, int i) {
+    return (masks[step * MW + (i >> 5)] >> (i & 31)) & 1u;
+}
+
+// broadcast-read the MP values of chain n from LDS and dot them with row[] (registers)
+template <int MP>
+__device__ __forceinline__ float lds_dot(const float *lds, int n, const float *row) {
+    const float4 *l4 = reinterpret_cast<const float4 *>(lds + n * MP);
+    float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+    for (int q = 0; q < MP / 4; ++q) {
+        float4 v = l4[q];
+        acc0 = fmaf(row[4 * q + 0], v.x, acc0);
+        acc1 = fmaf(row[4 * q + 1], v.y, acc1);
+        acc0 = fmaf(row[4 * q + 2], v.z, acc0);
+        acc1 = fmaf(row[4 * q + 3], v.w, acc1);
+    }
+    return acc0 + acc1;
+}
+
+// ---------------------------------------------------------------------------------------
+// residual, masks, F and dense J~ at every (b, t)
+// ---------------------------------------------------------------------------------------
+template <int MP>
+__global__ __launch_bounds__(64) void k_resjac_plrnn(const float *__restrict__ A, const float *__restrict__ W,
+                                                     const float *__restrict__ h, float alpha, int N,
+                                                     const float *__restrict__ x, const float *__restrict__ z0,
+                                                     const float *__restrict__ z, float *__restrict__ F_out,
+                                                     float *__restrict__ r_out, float *__restrict__ J_out,
+                                                     uint32_t *__restrict__ masks, const int *__restrict__ active,
+                                                     int B, int T, int M) {
+    using G = Geo<MP>;
+    __shared__ __align__(16) float lds[64];
+    const int lane = threadIdx.x;
+    const int n = lane / MP, i = lane % MP;
+    float wrow[MP];
+#pragma unroll
+    for (int j = 0; j < MP; ++j) wrow[j] = (i < M && j < M) ? W[i * M + j] : 0.f;
+    const float Ai = i < M ? A[i] : 0.f;
+    const float hi = (h && i < M) ? h[i] : 0.f;
+    const long total = (long)B * T;
+    const long ngroups = (total + G::NCH - 1) / G::NCH;
+    for (long grp = blockIdx.x; grp < ngroups; grp += gridDim.x) {
+        const long row = grp * G::NCH + n;
+        const bool in = row < total;
+        const int b = in ? (int)(row / T) : 0, s = in ? (int)(row % T) : 0;
+        const bool act = in && i < M && (!active || active[b]);
+        const float zt = act ? forced_state(x, z0, z, b, s, i, T, M, N, alpha) : 0.f;
+        const bool pos = zt > 0.f;
+        const uint64_t bal = __ballot(pos);
+        lds[lane] = pos ? zt : 0.f;
+        __syncthreads();
+        const float F = fmaf(Ai, zt, lds_dot<MP>(lds, n, wrow)) + hi;
+        __syncthreads();
+        if (act) {
+            const size_t e = (size_t)row * M + i;
+            if (r_out) r_out[e] = z[e] - F;
+            if (F_out) F_out[e] = F;
+            if (J_out) {
+                float *Jr = J_out + ((size_t)row * M + i) * M;
+#pragma unroll
+                for (int j = 0; j < MP; ++j) {
+                    if (j < M) {
+                        const float mj = (float)((bal >> (n * MP + j)) & 1ull);
+                        const float v = (j == i ? Ai : 0.f) + wrow[j] * mj;
+                        Jr[j] = v * p_of(j, N, alpha);
+                    }
+                }
+            }
+        }
+        if (masks && in && i == 0 && (!active || active[b])) {
+            if (MP == 64) {
+                masks[(size_t)row * 2 + 0] = (uint32_t)bal;
+                if (M > 32) masks[(size_t)row * 2 + 1] = (uint32_t)(bal >> 32);
+            } else {
+                const uint64_t seg = bal >> (n * MP);
+                masks[row] = (uint32_t)(MP == 32 ? seg : (seg & 0xffffull));
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// chunk aggregates.  Product over the step range [lo, hi) of the chain:
+//   forward: P_c = J~_{s1-1} ... J~_{s0}           v_c = Delta_{s1-1} from a zero carry
+//   reverse: P_c = J~_{s1} ... J~_{s0+1}  (then read transposed)
+//            v_c = lam_{s0} of the chunk from lam_{s1} = 0
+// MFMA formulation of P <- J~ P = diag(A p) P + (W diag(p)) (diag(m) P):
+//   A operand = W diag(p) (constant, registers), B operand = the masked accumulator itself
+//   (with the k-permutation kappa(4j+q, g) = 16j + 4g + q the 16x16x4 output layout is
+//   exactly the B layout of the next step, so no data moves between steps).
+// ---------------------------------------------------------------------------------------
+template <int MP, bool REV>
+__global__ __launch_bounds__(64) void k_chunk_product_plrnn(
+    const float *__restrict__ A, const float *__restrict__ W, float alpha, int N, const uint32_t *__restrict__ masks,
+    const float *__restrict__ rhs, const float *__restrict__ z, const float *__restrict__ x, float seed_scale,
+    float *__restrict__ Pout, float *__restrict__ vout, const int *__restrict__ active, int B, int T, int M, int C,
+    int ncs) {
+    using G = Geo<MP>;
+    constexpr int NCH = G::NCH, NI = G::NI, NS = G::NS, MW = G::MW;
+    __shared__ __align__(16) float lds[64];
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int nchains = B * ncs;
+    const int chain0 = blockIdx.x * NCH;
+
+    int pb[NCH], plo[NCH], plen[NCH], us0[NCH], us1[NCH];
+    int maxlen = 0;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n) {
+        const int id = chain0 + n;
+        bool ok = id < nchains;
+        const int b = ok ? id / ncs : 0, cc = ok ? id % ncs : 0;
+        ok = ok && (!active || active[b]);
+        const int s0 = cc * C, s1 = min(s0 + C, T);
+        const int lo = REV ? s0 + 1 : s0;
+        const int hi = REV ? min(s1 + 1, T) : s1;
+        pb[n] = b;
+        plo[n] = lo;
+        plen[n] = ok ? max(hi - lo, 0) : 0;
+        us0[n] = s0;
+        us1[n] = ok ? s1 : s0;
+        maxlen = max(maxlen, max(plen[n], us1[n] - us0[n]));
+    }
+
+    // A operand: (W diag(p))[16I + c][16j + 4g + q]
+    float Aop[NI][NS];
+#pragma unroll
+    for (int I = 0; I < NI; ++I)
+#pragma unroll
+        for (int j = 0; j < NS / 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int row = 16 * I + c, col = 16 * j + 4 * g + q;
+                Aop[I][4 * j + q] = (row < M && col < M) ? W[row * M + col] * p_of(col, N, alpha) : 0.f;
+            }
+    float dI[NI][4];
+#pragma unroll
+    for (int I = 0; I < NI; ++I)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * I + 4 * g + r;
+            dI[I][r] = row < M ? A[row] * p_of(row, N, alpha) : 0.f;
+        }
+    // accumulators start at the identity of each chain
+    v4f acc[NI][4];
+#pragma unroll
+    for (int Jt = 0; Jt < 4; ++Jt) {
+        const int n = (16 * Jt) / MP;
+        const int col = 16 * Jt + c - n * MP;
+#pragma unroll
+        for (int I = 0; I < NI; ++I)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[I][Jt][r] = (16 * I + 4 * g + r == col) ? 1.f : 0.f;
+    }
+
+    // VALU chain for v_c: lane = (chain un, row ui)
+    const int un = lane / MP, ui = lane % MP;
+    float wv[MP];
+    float du = 0.f, pu = 0.f, Au = 0.f;
+    if (!REV) {
+#pragma unroll
+        for (int k = 0; k < MP; ++k) wv[k] = (ui < M && k < M) ? W[ui * M + k] * p_of(k, N, alpha) : 0.f;
+        du = ui < M ? A[ui] * p_of(ui, N, alpha) : 0.f;
+    } else {
+#pragma unroll
+        for (int k = 0; k < MP; ++k) wv[k] = (ui < M && k < M) ? W[k * M + ui] : 0.f;
+        pu = p_of(ui, N, alpha);
+        Au = ui < M ? A[ui] : 0.f;
+    }
+    int ub = 0, ulo = 0, uhi = 0;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n)
+        if (n == un) { ub = pb[n]; ulo = us0[n]; uhi = us1[n]; }
+    float u = 0.f;
+
+    for (int t = 0; t < maxlen; ++t) {
+        // ---- matrix-core part: one step of every chain whose product is still running
+#pragma unroll
+        for (int Jt = 0; Jt < 4; ++Jt) {
+            const int n = (16 * Jt) / MP;
+            if (t < plen[n]) {
+                const size_t step = (size_t)pb[n] * T + plo[n] + t;
+                const uint32_t w0 = masks[step * MW];
+                const uint32_t w1 = MW > 1 ? masks[step * MW + 1] : 0u;
+                float Bop[NS];
+#pragma unroll
+                for (int j = 0; j < NS / 4; ++j) {
+                    const uint32_t wj = (j >> 1) ? w1 : w0;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) Bop[4 * j + q] = select_bit(wj, 16 * (j & 1) + 4 * g + q, acc[j][Jt][q]);
+                }
+#pragma unroll
+                for (int I = 0; I < NI; ++I)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[I][Jt][r] *= dI[I][r];
+#pragma unroll
+                for (int I = 0; I < NI; ++I)
+#pragma unroll
+                    for (int s = 0; s < NS; ++s) acc[I][Jt] = mfma16x16x4(Aop[I][s], Bop[s], acc[I][Jt]);
+            }
+        }
+        // ---- VALU part: local solution of the chunk
+        const bool run = ulo + t < uhi;
+        if (!REV) {
+            const int s = ulo + t;
+            const size_t step = (size_t)ub * T + s;
+            float w = 0.f;
+            if (run && ui < M) w = mask_bit(masks, step, MW, ui) ? u : 0.f;
+            lds[lane] = w;
+            __syncthreads();
+            const float y = fmaf(du, u, lds_dot<MP>(lds, un, wv));
+            __syncthreads();
+            if (run && ui < M) u = y - rhs[step * M + ui];
+        } else {
+            const int k = uhi - 1 - t;    // lam_k = J~_{k+1}^T lam_{k+1} + g_k
+            lds[lane] = u;
+            __syncthreads();
+            const float wt = lds_dot<MP>(lds, un, wv);
+            __syncthreads();
+            if (run && ui < M) {
+                const size_t step = (size_t)ub * T + k;
+                float y = 0.f;
+                if (t > 0) {
+                    const float m = (float)mask_bit(masks, step + 1, MW, ui);
+                    y = pu * fmaf(Au, u, m * wt);
+                }
+                float gk;
+                if (rhs) gk = rhs[step * M + ui];
+                else gk = ui < N ? seed_scale * (z[step * M + ui] - x[((size_t)ub * (T + 1) + k + 1) * N + ui]) : 0.f;
+                u = y + gk;
+            }
+        }
+    }
+
+    // ---- write the aggregates
+#pragma unroll
+    for (int Jt = 0; Jt < 4; ++Jt) {
+        const int n = (16 * Jt) / MP;
+        const int id = chain0 + n;
+        if (id < nchains && (plen[n] > 0 || us1[n] > us0[n])) {
+            const int col = 16 * Jt + c - n * MP;
+            float *P = Pout + (size_t)id * MP * MP;
+#pragma unroll
+            for (int I = 0; I < NI; ++I)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) P[(16 * I + 4 * g + r) * MP + col] = acc[I][Jt][r];
+        }
+    }
+    {
+        const int id = chain0 + un;
+        if (id < nchains) vout[(size_t)id * MP + ui] = u;
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// carries across chunks (one block of MP lanes per sequence)
+//   forward: carry_in[c] = y_end(c-1),  y_end(c) = P_c y_end(c-1) + v_c
+//   reverse: carry_in[c] = lam_{s1(c)}, lam_{s0(c)} = P_c^T lam_{s1(c)} + v_c
+// ---------------------------------------------------------------------------------------
+template <int MP, bool REV>
+__global__ __launch_bounds__(MP) void k_carry(const float *__restrict__ P, const float *__restrict__ v,
+                                              float *__restrict__ carry_in, const int *__restrict__ active,
+                                              uint32_t *__restrict__ norm_bits, int ncs) {
+    __shared__ __align__(16) float cs[MP];
+    const int b = blockIdx.x, i = threadIdx.x;
+    if (norm_bits && i == 0) norm_bits[b] = 0u;
+    if (active && !active[b]) return;
+    float cur = 0.f;
+    float pr[MP], pn[MP];
+    auto load = [&](int step, float *dst) {
+        const int cc = REV ? ncs - 1 - step : step;
+        const float *Pc = P + ((size_t)b * ncs + cc) * MP * MP;
+        if (!REV) {
+            const float4 *r4 = reinterpret_cast<const float4 *>(Pc + i * MP);
+#pragma unroll
+            for (int q = 0; q < MP / 4; ++q) {
+                float4 t = r4[q];
+                dst[4 * q] = t.x; dst[4 * q + 1] = t.y; dst[4 * q + 2] = t.z; dst[4 * q + 3] = t.w;
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < MP; ++k) dst[k] = Pc[k * MP + i];
+        }
+    };
+    load(0, pr);
+    for (int step = 0; step < ncs; ++step) {
+        const int cc = REV ? ncs - 1 - step : step;
+        const size_t id = (size_t)b * ncs + cc;
+        if (step + 1 < ncs) load(step + 1, pn);
+        const float vv = v[id * MP + i];
+        carry_in[id * MP + i] = cur;
+        cs[i] = cur;
+        __syncthreads();
+        float a0 = vv, a1 = 0.f;
+#pragma unroll
+        for (int k = 0; k < MP; k += 2) {
+            a0 = fmaf(pr[k], cs[k], a0);
+            a1 = fmaf(pr[k + 1], cs[k + 1], a1);
+        }
+        __syncthreads();
+        cur = a0 + a1;
+#pragma unroll
+        for (int k = 0; k < MP; ++k) pr[k] = pn[k];
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// forward fix-up: Delta from the carry, z += Delta, per-sequence max |Delta|
+// ---------------------------------------------------------------------------------------
+template <int MP>
+__global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict__ A, const float *__restrict__ W,
+                                                        float alpha, int N, const uint32_t *__restrict__ masks,
+                                                        const float *__restrict__ r, const float *__restrict__ carry_in,
+                                                        float *__restrict__ z, uint32_t *__restrict__ norm_bits,
+                                                        const int *__restrict__ active, int B, int T, int M, int C,
+                                                        int ncs) {
+    using G = Geo<MP>;
+    __shared__ __align__(16) float lds[64];
+    const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
+    const int id = blockIdx.x * G::NCH + n;
+    const bool ok0 = id < B * ncs;
+    const int b = ok0 ? id / ncs : 0, cc = ok0 ? id % ncs : 0;
+    const bool ok = ok0 && (!active || active[b]);
+    const int s0 = cc * C, len = ok ? min(C, T - s0) : 0;
+    float wrow[MP];
+#pragma unroll
+    for (int k = 0; k < MP; ++k) wrow[k] = (i < M && k < M) ? W[i * M + k] * p_of(k, N, alpha) : 0.f;
+    const float d = i < M ? A[i] * p_of(i, N, alpha) : 0.f;
+    float D = (ok && i < M) ? carry_in[(size_t)id * MP + i] : 0.f;
+    uint32_t emax = 0u;
+    const int maxlen = __builtin_amdgcn_readfirstlane(C);
+    for (int t = 0; t < maxlen; ++t) {
+        const bool run = t < len && i < M;
+        const size_t step = (size_t)b * T + s0 + t;
+        lds[lane] = (run && mask_bit(masks, step, G::MW, i)) ? D : 0.f;
+        __syncthreads();
+        const float y = fmaf(d, D, lds_dot<MP>(lds, n, wrow));
+        __syncthreads();
+        if (run) {
+            D = y - r[step * M + i];
+            const size_t e = step * M + i;
+            z[e] = z[e] + D;
+            const uint32_t ab = abs_bits(D);
+            emax = emax > ab ? emax : ab;
+        }
+    }
+    // max over the MP lanes of this chain
+#pragma unroll
+    for (int off = MP / 2; off > 0; off >>= 1) {
+        const uint32_t o = (uint32_t)__shfl_xor((int)emax, off, 64);
+        emax = emax > o ? emax : o;
+    }
+    if (ok && i == 0) atomicMax(norm_bits + b, emax);
+}
+
+// ---------------------------------------------------------------------------------------
+// reverse fix-up: lam from the carry, written out, with the parameter-gradient partial
+// sums of this chunk: dW[i][j] += lam_i relu(z~_j), dA_i += lam_i z~_i, dh_i += lam_i
+// (layout gpart[chain][MP][MP + 2]).
+// ---------------------------------------------------------------------------------------
+template <int MP>
+__global__ __launch_bounds__(64) void k_fixup_rev_plrnn(const float *__restrict__ A, const float *__restrict__ W,
+                                                        float alpha, int N, const uint32_t *__restrict__ masks,
+                                                        const float *__restrict__ gin, float seed_scale,
+                                                        const float *__restrict__ x, const float *__restrict__ z0,
+                                                        const float *__restrict__ z, const float *__restrict__ carry_in,
+                                                        float *__restrict__ lam_out, float *__restrict__ gpart, int B,
+                                                        int T, int M, int C, int ncs) {
+    using G = Geo<MP>;
+    __shared__ __align__(16) float lds[64];
+    const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
+    const int id = blockIdx.x * G::NCH + n;
+    const bool ok = id < B * ncs;
+    const int b = ok ? id / ncs : 0, cc = ok ? id % ncs : 0;
+    const int s0 = cc * C, s1 = ok ? min(s0 + C, T) : s0;
+    float wcol[MP], dW[MP];
+#pragma unroll
+    for (int k = 0; k < MP; ++k) {
+        wcol[k] = (i < M && k < M) ? W[k * M + i] : 0.f;
+        dW[k] = 0.f;
+    }
+    const float pi = p_of(i, N, alpha), Ai = i < M ? A[i] : 0.f;
+    float lam = (ok && i < M) ? carry_in[(size_t)id * MP + i] : 0.f;
+    float dA = 0.f, dh = 0.f;
+    const int maxlen = __builtin_amdgcn_readfirstlane(C);
+    for (int t = 0; t < maxlen; ++t) {
+        const int k = s1 - 1 - t;
+        const bool run = k >= s0 && i < M;
+        lds[lane] = lam;
+        __syncthreads();
+        const float wt = lds_dot<MP>(lds, n, wcol);
+        __syncthreads();
+        float zt = 0.f;
+        if (run) {
+            const size_t step = (size_t)b * T + k;
+            float y = 0.f;
+            if (k + 1 < T) {
+                const float m = (float)mask_bit(masks, step + 1, G::MW, i);
+                y = pi * fmaf(Ai, lam, m * wt);
+            }
+            float gk;
+            if (gin) gk = gin[step * M + i];
+            else gk = i < N ? seed_scale * (z[step * M + i] - x[((size_t)b * (T + 1) + k + 1) * N + i]) : 0.f;
+            lam = y + gk;
+            if (lam_out) lam_out[step * M + i] = lam;
+            zt = forced_state(x, z0, z, b, k, i, T, M, N, alpha);
+            dA = fmaf(lam, zt, dA);
+            dh += lam;
+        }
+        const float lr = run ? lam : 0.f;
+        lds[lane] = (run && zt > 0.f) ? zt : 0.f;
+        __syncthreads();
+        const float4 *l4 = reinterpret_cast<const float4 *>(lds + n * MP);
+#pragma unroll
+        for (int q = 0; q < MP / 4; ++q) {
+            const float4 v = l4[q];
+            dW[4 * q + 0] = fmaf(lr, v.x, dW[4 * q + 0]);
+            dW[4 * q + 1] = fmaf(lr, v.y, dW[4 * q + 1]);
+            dW[4 * q + 2] = fmaf(lr, v.z, dW[4 * q + 2]);
+            dW[4 * q + 3] = fmaf(lr, v.w, dW[4 * q + 3]);
+        }
+        __syncthreads();
+    }
+    if (ok) {
+        float *gp = gpart + ((size_t)id * MP + i) * (MP + 2);
+#pragma unroll
+        for (int k = 0; k < MP; ++k) gp[k] = dW[k];
+        gp[MP] = dA;
+        gp[MP + 1] = dh;
+    }
+}
+
+// sum the per-chunk partials in float64: one thread per entry of [MP][MP + 2]
+__global__ void k_reduce_gpart(const float *__restrict__ gpart, int nchains, int MP, int M, float *__restrict__ dA,
+                               float *__restrict__ dW, float *__restrict__ dh) {
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    const int stride = MP * (MP + 2);
+    if (e >= stride) return;
+    const int i = e / (MP + 2), j = e % (MP + 2);
+    if (i >= M) return;
+    if (j < MP && j >= M) return;
+    double s0 = 0.0, s1 = 0.0;
+    int ch = 0;
+    for (; ch + 1 < nchains; ch += 2) {
+        s0 += (double)gpart[(size_t)ch * stride + e];
+        s1 += (double)gpart[(size_t)(ch + 1) * stride + e];
+    }
+    if (ch < nchains) s0 += (double)gpart[(size_t)ch * stride + e];
+    const float v = (float)(s0 + s1);
+    if (j < MP) {
+        if (dW) dW[i * M + j] = v;
+    } else if (j == MP) {
+        if (dA) dA[i] = v;
+    } else {
+        if (dh) dh[i] = v;
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// host launchers
+// ---------------------------------------------------------------------------------------
+static int padded(int M) { return M <= 16 ? 16 : (M <= 32 ? 32 : 64); }
+
+int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, float *J, uint32_t *masks,
+                        const int *active, hipStream_t st) {
+    const int MP = padded(a.M);
+    const long groups = ((long)a.B * a.T + (64 / MP) - 1) / (64 / MP);
+    const int grid = (int)(groups < 16384 ? groups : 16384);
+#define RJ(MPV)                                                                                                   \
+    hipLaunchKernelGGL(k_resjac_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, z, \
+                       F, r, J, masks, active, a.B, a.T, a.M)
+    if (MP == 16) RJ(16); else if (MP == 32) RJ(32); else RJ(64);
+#undef RJ
+    DEER_LAUNCH_CHECK("k_resjac_plrnn");
+    return DEER_OK;
+}
+
+int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *masks, const float *rhs, const float *z,
+                               float seed_scale, float *P, float *v, const int *active, int C, int ncs,
+                               hipStream_t st) {
+    const int MP = padded(a.M);
+    const int nch = a.B * ncs;
+    const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+#define CP(MPV, R)                                                                                                  \
+    hipLaunchKernelGGL((k_chunk_product_plrnn<MPV, R>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, \
+                       rhs, z, a.x, seed_scale, P, v, active, a.B, a.T, a.M, C, ncs)
+    if (!rev) {
+        if (MP == 16) CP(16, false); else if (MP == 32) CP(32, false); else CP(64, false);
+    } else {
+        if (MP == 16) CP(16, true); else if (MP == 32) CP(32, true); else CP(64, true);
+    }
+#undef CP
+    DEER_LAUNCH_CHECK("k_chunk_product_plrnn");
+    return DEER_OK;
+}
+
+int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
+                 uint32_t *norm_bits, int B, int ncs, hipStream_t st) {
+#define CA(MPV, R) \
+    hipLaunchKernelGGL((k_carry<MPV, R>), dim3(B), dim3(MPV), 0, st, P, v, carry_in, active, norm_bits, ncs)
+    if (!rev) {
+        if (MP == 16) CA(16, false); else if (MP == 32) CA(32, false); else CA(64, false);
+    } else {
+        if (MP == 16) CA(16, true); else if (MP == 32) CA(32, true); else CA(64, true);
+    }
+#undef CA
+    DEER_LAUNCH_CHECK("k_carry");
+    return DEER_OK;
+}
+
+int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in, float *z,
+                           uint32_t *norm_bits, const int *active, int C, int ncs, hipStream_t st) {
+    const int MP = padded(a.M);
+    const int nch = a.B * ncs;
+    const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+#define FX(MPV)                                                                                                       \
+    hipLaunchKernelGGL(k_fixup_fwd_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, carry_in, \
+                       z, norm_bits, active, a.B, a.T, a.M, C, ncs)
+    if (MP == 16) FX(16); else if (MP == 32) FX(32); else FX(64);
+#undef FX
+    DEER_LAUNCH_CHECK("k_fixup_fwd_plrnn");
+    return DEER_OK;
+}
+
+int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *g, float seed_scale, const float *z,
+                           const float *carry_in, float *lam, float *gpart, int C, int ncs, hipStream_t st) {
+    const int MP = padded(a.M);
+    const int nch = a.B * ncs;
+    const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+#define FR(MPV)                                                                                                     \
+    hipLaunchKernelGGL(k_fixup_rev_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, g,       \
+                       seed_scale, a.x, a.z0, z, carry_in, lam, gpart, a.B, a.T, a.M, C, ncs)
+    if (MP == 16) FR(16); else if (MP == 32) FR(32); else FR(64);
+#undef FR
+    DEER_LAUNCH_CHECK("k_fixup_rev_plrnn");
+    return DEER_OK;
+}
+
+int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *dA, float *dW, float *dh,
+                        hipStream_t st) {
+    const int n = MP * (MP + 2);
+    hipLaunchKernelGGL(k_reduce_gpart, dim3((n + 255) / 256), dim3(256), 0, st, gpart, nchains, MP, M, dA, dW, dh);
+    DEER_LAUNCH_CHECK("k_reduce_gpart");
+    return DEER_OK;
+}
+
+int padded_dim(int M) { return padded(M); }
+
+}  // namespace deer

@@ -1,0 +1,45 @@
+// Internal launcher interface between the C-ABI layer and the kernel translation units.
+#pragma once
+#include "common.h"
+
+namespace deer {
+
+struct PlrnnArgs {
+    const float *A, *W, *h;
+    float alpha;
+    int N;
+    const float *x, *z0;
+    int B, T, M;
+};
+
+int padded_dim(int M);
+
+// vanilla PLRNN
+int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, float *J, uint32_t *masks,
+                        const int *active, hipStream_t st);
+int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *masks, const float *rhs, const float *z,
+                               float seed_scale, float *P, float *v, const int *active, int C, int ncs,
+                               hipStream_t st);
+int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
+                 uint32_t *norm_bits, int B, int ncs, hipStream_t st);
+int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in, float *z,
+                           uint32_t *norm_bits, const int *active, int C, int ncs, hipStream_t st);
+int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *g, float seed_scale, const float *z,
+                           const float *carry_in, float *lam, float *gpart, int C, int ncs, hipStream_t st);
+int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *dA, float *dW, float *dh,
+                        hipStream_t st);
+
+// diagonal complex scan
+size_t diag_scan_ws_bytes(int B, int T, int M);
+int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const float *b, const float *Bc, int K,
+                     const float *u, float *y, void *ws, hipStream_t st);
+size_t diag_grads_ws_bytes(int B, int T, int M);
+int launch_diag_grads(int B, int T, int M, int K, const float *a, const float *h, const float *x, float *dlam,
+                      float *dBc, void *ws, hipStream_t st);
+
+// small utilities
+int launch_fill_teacher(int B, int T, int M, int N, const float *x, float *z, hipStream_t st);
+int launch_fill_i32(int *p, int n, int v, hipStream_t st);
+int launch_fill_f32(float *p, size_t n, float v, hipStream_t st);
+
+}  // namespace deer

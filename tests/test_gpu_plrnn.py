@@ -1,0 +1,202 @@
+"""Vanilla PLRNN GTF-DEER on the GPU against the float64 oracle (through the C ABI).
+
+Tolerance: 1e-4 normwise relative error for float32 states, adjoints and gradients;
+bit-exact ReLU masks when both sides take the decision in float32 on the same input.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from gpu_util import masks_to_bool, oracle_model, rel_inf, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2605_12683_amd as D  # noqa: E402
+
+TOL = 1e-4
+
+
+@pytest.fixture(autouse=True)
+def _no_chunk_override():
+    os.environ.pop("DEER_CHUNK", None)
+    yield
+    os.environ.pop("DEER_CHUNK", None)
+
+
+def _case(M, N, B, T, alpha, seed, w_std=None):
+    """A random vanilla PLRNN; by default a contraction (A in [0.3, 0.75], ||W||_2 = 0.2) so
+    that the trajectory stays O(1) for any M and N."""
+    if w_std is not None:
+        return W.random_plrnn_case(M, N, B, T, alpha, seed, w_std=w_std)
+    return W.random_plrnn_case(M, N, B, T, alpha, seed, w_norm=0.2, a_range=(0.3, 0.75))
+
+
+@pytest.mark.parametrize("M,N,T", [(1, 1, 50), (3, 3, 100), (16, 3, 257), (17, 5, 130), (33, 33, 64), (64, 64, 100)])
+def test_jacobian_masks_residual(M, N, T):
+    c = _case(M, N, 2, T, 0.2, 100 + M)
+    m = oracle_model(c)
+    z = np.random.default_rng(1).standard_normal((2, T, M)).astype(np.float32)
+    say("plrnn_jacobian", M, N, T)
+    out = D.plrnn_jacobian(m, c.x, z, c.alpha, N, want=("F", "r", "masks"), dense_J=True)
+    torch.cuda.synchronize()
+    ref = O.jacobian_at(m, c.x, z, c.alpha, N, mask_precision="float32",
+                        dense_index=[(b, t) for b in range(2) for t in range(T)])
+    got_mask = masks_to_bool(out["masks"].cpu().numpy(), M)
+    assert np.array_equal(got_mask, ref["mask"])
+    assert rel_inf(out["F"].cpu().numpy(), ref["F"]) < 1e-5
+    assert rel_inf(out["r"].cpu().numpy(), ref["r"]) < 1e-5
+    assert rel_inf(out["J"].cpu().numpy().reshape(-1, M, M), ref["J"]) < 1e-6
+
+
+def test_config1_fixed_five_iterations():
+    """Workload 1 (vanilla PLRNN M=3, T=1024): exactly 5 Newton updates from the teacher states."""
+    c = W.make_config(1)
+    m = oracle_model(c)
+    say("deer_solve config1 fixed 5")
+    res = D.deer_solve(m, c.x, c.alpha, c.n_obs, fixed_iters=5)
+    ref = O.newton(m, c.x, c.alpha, c.n_obs, fixed_iters=5)
+    assert res["status"] == 0
+    assert rel_inf(res["z"].cpu().numpy(), ref["z"]) < TOL
+    assert res["iters"] == [5]
+
+
+@pytest.mark.parametrize("M,N,B,T,alpha,chunk", [
+    (3, 3, 1, 300, 0.1, 0), (3, 3, 2, 300, 0.1, 17), (16, 3, 3, 1000, 0.2, 0), (16, 3, 2, 777, 0.2, 64),
+    (20, 4, 2, 513, 0.3, 100), (32, 32, 2, 600, 0.1, 0), (40, 10, 2, 300, 0.3, 33), (64, 64, 2, 400, 0.05, 0),
+    (64, 64, 3, 1000, 0.05, 128), (5, 2, 4, 64, 0.5, 64), (16, 16, 1, 1, 0.2, 0), (8, 8, 2, 2, 0.2, 0)])
+def test_solve_reaches_rollout(M, N, B, T, alpha, chunk):
+    """Converged GTF-DEER equals the sequential GTF rollout (unique zero of the residual)."""
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    c = _case(M, N, B, T, alpha, 200 + M + T)
+    m = oracle_model(c)
+    say("deer_solve", M, N, B, T, alpha, chunk)
+    res = D.deer_solve(m, c.x, alpha, N, tol=1e-5, max_iter=100, want_masks=True)
+    assert res["status"] == 0, res
+    ref = O.rollout(m, c.x, alpha, N)
+    z = res["z"].cpu().numpy()
+    assert rel_inf(z, ref) < TOL
+    assert all(1 <= k <= 100 for k in res["iters"])
+    assert all(n < 1e-5 for n in res["norms"])
+    # masks at the returned z: equal to the fixed point's outside a tie band
+    _, _, _, zt = O.residual_and_masks(m, c.x, ref, alpha, N)
+    got = masks_to_bool(res["masks"].cpu().numpy(), M)
+    far = np.abs(zt) > 1e-4 * np.abs(zt).max()
+    assert np.array_equal(got[far], (zt > 0)[far])
+
+
+def test_iteration_counts_match_oracle():
+    c = _case(16, 3, 4, 800, 0.2, 7)
+    m = oracle_model(c)
+    say("deer_solve iteration counts")
+    res = D.deer_solve(m, c.x, 0.2, 3, tol=1e-5)
+    ref = O.newton(m, c.x, 0.2, 3, tol=1e-5)
+    assert max(abs(a - b) for a, b in zip(res["iters"], ref["iters"].tolist())) <= 1
+
+
+def test_alpha1_full_observation_two_updates():
+    """alpha = 1, M <= N: z* = F(zbar) in closed form; the GPU stops after 2 updates."""
+    c = _case(6, 6, 3, 500, 1.0, 11, w_std=0.8)
+    m = oracle_model(c)
+    say("deer_solve alpha=1")
+    res = D.deer_solve(m, c.x, 1.0, 6, tol=1e-5)
+    closed = O.model_map(m, c.x[:, :-1].astype(np.float64))
+    assert rel_inf(res["z"].cpu().numpy(), closed) < 1e-6
+    assert res["iters"] == [2, 2, 2]
+
+
+def test_alpha0_linear_model_two_updates():
+    M, T = 8, 700
+    rng = np.random.default_rng(3)
+    m = {"kind": "plrnn", "A": rng.uniform(0.5, 0.9, M).astype(np.float32), "W": np.zeros((M, M), np.float32),
+         "h": rng.normal(0, 0.1, M).astype(np.float32)}
+    x = rng.standard_normal((2, T + 1, M)).astype(np.float32)
+    say("deer_solve alpha=0 linear")
+    res = D.deer_solve(m, x, 0.0, M, tol=1e-6)
+    assert res["iters"] == [2, 2]
+    assert rel_inf(res["z"].cpu().numpy(), O.rollout(m, x, 0.0, M)) < 1e-5
+
+
+def test_user_init_and_z0():
+    c = _case(16, 3, 2, 400, 0.2, 13)
+    m = oracle_model(c)
+    z0 = np.random.default_rng(5).standard_normal((2, 16)).astype(np.float32)
+    ref = O.rollout(m, c.x, 0.2, 3, z0=z0)
+    zinit = torch.tensor(ref.astype(np.float32) + 0.1, device="cuda")
+    say("deer_solve user init + z0")
+    res = D.deer_solve(m, c.x, 0.2, 3, z0=z0, init="user", z=zinit, tol=1e-6)
+    assert rel_inf(res["z"].cpu().numpy(), ref) < TOL
+    res = D.deer_solve(m, c.x, 0.2, 3, z0=z0, init="zero", tol=1e-6)
+    assert rel_inf(res["z"].cpu().numpy(), ref) < TOL
+
+
+def test_nonfinite_and_not_converged():
+    c = _case(8, 3, 2, 200, 0.2, 17)
+    m = oracle_model(c)
+    x = c.x.copy()
+    x[1, 50, 0] = np.nan
+    say("deer_solve NaN input")
+    res = D.deer_solve(m, x, 0.2, 3, tol=1e-5, check=False)
+    assert res["status"] == 3                      # DEER_ERR_NONFINITE
+    say("deer_solve max_iter=1")
+    res = D.deer_solve(m, c.x, 0.2, 3, tol=1e-5, max_iter=1, check=False)
+    assert res["status"] == 2                      # DEER_ERR_NOT_CONVERGED
+    assert res["iters"] == [1, 1]
+
+
+@pytest.mark.parametrize("M,N,B,T,alpha,chunk", [(3, 3, 1, 300, 0.1, 0), (16, 3, 3, 1000, 0.2, 0),
+                                                 (16, 3, 2, 777, 0.2, 64), (20, 4, 2, 513, 0.3, 100),
+                                                 (64, 64, 2, 400, 0.05, 0), (40, 10, 2, 300, 0.3, 33),
+                                                 (8, 8, 1, 1, 0.2, 0)])
+def test_adjoint_and_grads(M, N, B, T, alpha, chunk):
+    """lam and dL/dtheta at the same float32 trajectory (the oracle's fixed point rounded to
+    float32); both sides take the ReLU decision in float32."""
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    c = _case(M, N, B, T, alpha, 300 + M + T)
+    m = oracle_model(c)
+    z32 = O.rollout(m, c.x, alpha, N).astype(np.float32)
+    say("deer_adjoint", M, N, B, T, alpha, chunk)
+    out = D.deer_adjoint(m, c.x, z32, alpha, N)
+    lam_ref = O.adjoint(m, c.x, z32, alpha, N, mask_precision="float32")
+    g_ref = O.param_grads(m, c.x, z32, alpha, N, lam_ref, mask_precision="float32")
+    assert rel_inf(out["lam"].cpu().numpy(), lam_ref) < TOL
+    for k in ("A", "W", "h"):
+        assert rel_inf(out["grads"][k].cpu().numpy(), g_ref[k]) < TOL, k
+
+
+def test_adjoint_user_cotangent():
+    c = _case(16, 3, 2, 300, 0.2, 19)
+    m = oracle_model(c)
+    z32 = O.rollout(m, c.x, 0.2, 3).astype(np.float32)
+    g = np.random.default_rng(2).standard_normal(z32.shape).astype(np.float32)
+    say("deer_adjoint user g")
+    out = D.deer_adjoint(m, c.x, z32, 0.2, 3, g=g)
+    lam_ref = O.adjoint(m, c.x, z32, 0.2, 3, g=g, mask_precision="float32")
+    assert rel_inf(out["lam"].cpu().numpy(), lam_ref) < TOL
+
+
+def test_config2_full_size():
+    """Workload 2 at full size (M=16, N=3, T=16384, B=16): solve, then adjoint + gradients."""
+    c = W.make_config(2)
+    m = oracle_model(c)
+    say("deer_solve config2 full")
+    res = D.deer_solve(m, c.x, c.alpha, c.n_obs, tol=c.tol)
+    assert res["status"] == 0
+    ref = O.rollout(m, c.x, c.alpha, c.n_obs)
+    assert rel_inf(res["z"].cpu().numpy(), ref) < TOL
+    z32 = ref.astype(np.float32)
+    say("deer_adjoint config2 full")
+    out = D.deer_adjoint(m, c.x, z32, c.alpha, c.n_obs)
+    lam_ref = O.adjoint(m, c.x, z32, c.alpha, c.n_obs, mask_precision="float32")
+    assert rel_inf(out["lam"].cpu().numpy(), lam_ref) < TOL
+    g_ref = O.param_grads(m, c.x, z32, c.alpha, c.n_obs, lam_ref, mask_precision="float32")
+    for k in ("A", "W", "h"):
+        assert rel_inf(out["grads"][k].cpu().numpy(), g_ref[k]) < TOL, k

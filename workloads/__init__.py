@@ -254,10 +254,15 @@ def make_config(i: int, B: int | None = None, T: int | None = None) -> Workload:
 
 
 def random_plrnn_case(M: int, n_obs: int, B: int, T: int, alpha: float, seed: int, w_std: float = 0.1,
-                      system: str = "lorenz63") -> Workload:
-    """Small vanilla-PLRNN case for tests (any M >= 1, any n_obs <= M)."""
+                      system: str = "lorenz63", w_norm: float | None = None, a_range=(0.5, 0.9)) -> Workload:
+    """Small vanilla-PLRNN case for tests (any M >= 1, any n_obs <= M).  With w_norm, W is
+    rescaled to that spectral norm (max A + w_norm < 1 makes the map a contraction)."""
     rng = np.random.default_rng(seed)
-    params = plrnn_params(M, rng, w_std=w_std)
+    params = plrnn_params(M, rng, a_range=a_range, w_std=w_std)
+    if w_norm is not None:
+        Wm = params["W"].astype(np.float64)
+        s = np.linalg.norm(Wm, 2)
+        params["W"] = (Wm * (w_norm / s if s > 0 else 1.0)).astype(np.float32)
     if system == "lorenz63" and n_obs <= 3:
         x = observed_batch("lorenz63", n_obs, B, T, seed + 1)
     else:

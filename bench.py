@@ -1,0 +1,214 @@
+#!/usr/bin/env python3
+"""Throughput of the GTF-DEER hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input:
+  PLRNN workloads: deer_solve (Newton loop: residual + Jacobian masks, chunked MFMA scan,
+                   carries, fix-up + max-norm test, until every sequence converged or the
+                   fixed iteration count) followed by deer_adjoint (MSE seed, reverse scan
+                   with transposed Jacobians, parameter-gradient reductions).
+  diagonal SSM:    deer_solve (fused input projection + forward complex scan) followed by
+                   deer_adjoint (reverse scan with conj(lambda) + dlambda / dBc reductions)
+                   on a fixed cotangent.
+Inputs are resident in HBM before the timed region.  The value is DEER timesteps per
+second: sum over sequences of T x Newton updates, per second of the whole step.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
+PEAK_FP32_MFMA_TFLOPS = 157.3    # MI355X dense fp32 matrix
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _plrnn_step(D, model, xd, c, ws_s, ws_a):
+    res = D.deer_solve(model, xd, c.alpha, c.n_obs, tol=c.tol, max_iter=c.max_iter, fixed_iters=c.fixed_iters,
+                       ws=ws_s)
+    D.deer_adjoint(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a)
+    return sum(res["iters"])
+
+
+def _diag_step(D, model, xd, c, ws_s, ws_a, g):
+    res = D.deer_solve(model, xd, 0.0, 0, ws=ws_s)
+    D.deer_adjoint(model, xd, res["z"], 0.0, 0, g=g, ws=ws_a)
+    return c.B
+
+
+def roofline_for(name, c, total_ms, launches, steps, iters_per_step):
+    """Algorithmic work of the dominant kernel over the timed region, divided by its time."""
+    B, T, M = c.B, c.T, c.M
+    if name == "k_chunk_product_plrnn":
+        # forward: every Newton update composes J~_t P for all T steps of each updated sequence;
+        # adjoint: the shifted products cover steps 1..T-1 of every sequence.  2 M^3 flop each.
+        units = steps * (iters_per_step * T + B * (T - 1))
+        work = units * 2.0 * M ** 3
+        ach = work / (total_ms * 1e-3) / 1e12
+        return {"bound": "mfma", "achieved": ach, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                "frac": ach / PEAK_FP32_MFMA_TFLOPS, "traffic": None,
+                "kernel": name, "avg_launch_ms": total_ms / launches,
+                "work_per_unit": f"{2 * M ** 3} flop per (b,t) step (2 M^3, J~_t P)",
+                "units_per_launch": units / launches}
+    if name in ("k_diag_chunk_fixup", "k_diag_chunk_reduce"):
+        # fix-up: read b (8 B) + write y (8 B) per complex element; the forward launch of the
+        # solve forms b from x on the fly (8 B written per element, 12 B of x per step)
+        per = 16.0 if name == "k_diag_chunk_fixup" else 8.0
+        units = launches * B * T * M
+        work = units * per
+        ach = work / (total_ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
+                "traffic": None, "kernel": name, "avg_launch_ms": total_ms / launches,
+                "work_per_unit": f"{per:g} B per complex element", "units_per_launch": units / launches}
+    if name in ("k_fixup_fwd_plrnn", "k_fixup_rev_plrnn", "k_resjac_plrnn"):
+        W = (M + 31) // 32
+        per = {"k_fixup_fwd_plrnn": 4 * W + 12 * M, "k_fixup_rev_plrnn": 4 * W + 8 * M + 4 * M,
+               "k_resjac_plrnn": 8 * M + 4 * W + 4 * M}[name]
+        units = steps * (iters_per_step * T + B * T) if name != "k_fixup_rev_plrnn" else steps * B * T
+        work = units * per
+        ach = work / (total_ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
+                "traffic": None, "kernel": name, "avg_launch_ms": total_ms / launches,
+                "work_per_unit": f"{per} B per (b,t) step", "units_per_launch": units / launches}
+    return {"bound": "unknown", "kernel": name, "avg_launch_ms": total_ms / launches, "achieved": None,
+            "peak": None, "unit": None, "frac": None, "traffic": None}
+
+
+def cpu_baseline(c, budget_s=20.0):
+    """The float64 oracle on the host, on a bounded sample of the same workload."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_limits
+        lim = threadpool_limits(1)
+    except Exception:       # pragma: no cover
+        lim = None
+    m = {"kind": c.kind, **c.params}
+    if c.kind == "diag_ssm":
+        Ts = min(c.T, 1 << 16)
+        xs = c.x[:1, :Ts + 1]
+        t0 = time.perf_counter()
+        O.diag_ssm_step(c.params, xs)
+        dt = time.perf_counter() - t0
+        value, sample = Ts / dt, f"1 of {c.B} sequences, first {Ts} of {c.T} steps, forward+read-out+reverse"
+    else:
+        # The oracle is vectorised over the batch and sequential in time: about 20 us per
+        # time step per Newton update.  Keep the whole batch, shorten T to fit the budget.
+        Ts = c.T
+        while Ts > 1024 and Ts * 10 * 20e-6 > budget_s:
+            Ts //= 2
+        xs = c.x[:, :Ts + 1]
+        t0 = time.perf_counter()
+        res = O.newton(m, xs, c.alpha, c.n_obs, tol=c.tol, max_iter=c.max_iter, fixed_iters=c.fixed_iters)
+        lam = O.adjoint(m, xs, res["z"], c.alpha, c.n_obs)
+        O.param_grads(m, xs, res["z"], c.alpha, c.n_obs, lam)
+        dt = time.perf_counter() - t0
+        value = float(np.sum(res["iters"]) * Ts) / dt
+        sample = f"all {c.B} sequences, first {Ts} of {c.T} steps, Newton solve + adjoint + gradients"
+    if lim is not None:
+        lim.unregister() if hasattr(lim, "unregister") else None
+    return {"value": value, "unit": "timesteps/s", "cores": 1, "kind": "oracle", "sample": sample,
+            "seconds": dt, "host_cpus": os.cpu_count()}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    import paper_2605_12683_amd as D
+    from paper_2605_12683_amd import _binding as Bnd
+
+    c = W.make_config(args.config)
+    log(f"[bench] workload {c.name}: B={c.B} T={c.T} M={c.M} kind={c.kind}")
+    dev = torch.device("cuda:0")
+    xd = torch.tensor(c.x, device=dev)
+    if c.kind == "diag_ssm":
+        model = D._Model({"kind": "diag_ssm", "lam": c.params["lam"], "Bc": c.params["Bc"]})
+        ws_s = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_SOLVE))
+        ws_a = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_ADJOINT))
+        gen = torch.Generator(device=dev).manual_seed(0)
+        g = torch.randn(c.B, c.T, c.M, 2, device=dev, generator=gen) * 1e-6
+        step = lambda: _diag_step(D, model, xd, c, ws_s, ws_a, g)          # noqa: E731
+    elif c.kind == "plrnn":
+        model = D._Model({"kind": "plrnn", **c.params})
+        ws_s = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_SOLVE))
+        ws_a = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_ADJOINT))
+        step = lambda: _plrnn_step(D, model, xd, c, ws_s, ws_a)            # noqa: E731
+    else:
+        print(f"workload {c.name}: model kind {c.kind} not supported by this build", file=sys.stderr)
+        sys.exit(3)
+
+    for i in range(args.warmup):
+        step()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    torch.cuda.synchronize()
+    Bnd.timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    updates = 0
+    for i in range(args.steps):
+        updates += step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kt = Bnd.timing_report()
+    Bnd.timing_enable(False)
+    dt = t1 - t0
+    iters_per_step = updates / args.steps
+    timesteps = updates * c.T
+    value = timesteps / dt
+    for k, (ms, n) in sorted(kt.items(), key=lambda kv: -kv[1][0]):
+        log(f"[bench] {k:28s} {ms:10.3f} ms total  {n:6d} launches  {ms / n:9.4f} ms avg")
+    dom = max(kt.items(), key=lambda kv: kv[1][0])
+    roof = roofline_for(dom[0], c, dom[1][0], dom[1][1], args.steps, iters_per_step)
+
+    out = {
+        "metric": "DEER timesteps/sec (B*T*Newton iters)",
+        "value": value,
+        "unit": "timesteps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": dt / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Lorenz trajectories, random-init parameters)",
+        "config": {"workload": c.name, "kind": c.kind, "B": c.B, "T": c.T, "M": c.M, "N": c.n_obs,
+                   "alpha": c.alpha, "tol": c.tol if not c.fixed_iters else None,
+                   "fixed_iters": c.fixed_iters or None, "newton_updates_per_step": iters_per_step,
+                   "step": "deer_solve + deer_adjoint"},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        cb = cpu_baseline(c)
+        out["cpu_baseline"] = cb
+        log(f"[bench] cpu oracle: {cb['value']:.4g} timesteps/s ({cb['sample']}, {cb['seconds']:.1f} s)")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

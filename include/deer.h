@@ -175,6 +175,16 @@ int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, cons
 /* Workspace bytes deer_scan needs. */
 size_t deer_scan_workspace_bytes(int layout, int B, int T, int M);
 
+/* Diagnostics: per-kernel timing with HIP events.  While enabled, every kernel launch is
+ * bracketed by two events recorded on the stream it is launched on (the caller's stream).
+ * deer_timing_enable(1) clears earlier records and starts recording; deer_timing_enable(0)
+ * stops.  deer_timing_report(idx, ...) waits for the events of the idx-th distinct kernel
+ * (in first-launch order) and returns its name, total milliseconds and launch count; the
+ * return value is the number of distinct kernels recorded (negative on a HIP error).
+ * Process-wide; meant for benchmarks, not for concurrent production calls. */
+int deer_timing_enable(int on);
+int deer_timing_report(int idx, char *name, int name_cap, double *ms_total, long *launches);
+
 /* Static description of a status code; never NULL. */
 const char *deer_status_string(int status);
 

@@ -21,7 +21,8 @@ DEER_OP_SOLVE, DEER_OP_ADJOINT = 0, 1
 DEER_SCAN_DENSE, DEER_SCAN_DIAG_C64 = 0, 1
 
 EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "plrnn_jacobian", "deer_scan",
-            "deer_scan_workspace_bytes", "deer_status_string", "deer_last_error"]
+            "deer_scan_workspace_bytes", "deer_status_string", "deer_last_error", "deer_timing_enable",
+            "deer_timing_report"]
 
 _fp = ctypes.c_void_p
 
@@ -76,8 +77,32 @@ def load(path: str = LIB_PATH):
     lib.deer_status_string.restype = ctypes.c_char_p
     lib.deer_last_error.argtypes = []
     lib.deer_last_error.restype = ctypes.c_char_p
+    lib.deer_timing_enable.argtypes = [i32]
+    lib.deer_timing_enable.restype = i32
+    lib.deer_timing_report.argtypes = [i32, ctypes.c_char_p, i32, P(ctypes.c_double), P(ctypes.c_long)]
+    lib.deer_timing_report.restype = i32
     _lib = lib
     return lib
+
+
+def timing_enable(on: bool):
+    load().deer_timing_enable(1 if on else 0)
+
+
+def timing_report() -> dict:
+    """{kernel name: (total ms, launches)} of the launches recorded since timing_enable(True)."""
+    lib = load()
+    n = lib.deer_timing_report(-1, None, 0, None, None)
+    if n < 0:
+        raise RuntimeError("deer_timing_report failed")
+    out = {}
+    for i in range(n):
+        buf = ctypes.create_string_buffer(128)
+        ms = ctypes.c_double()
+        cnt = ctypes.c_long()
+        lib.deer_timing_report(i, buf, 128, ctypes.byref(ms), ctypes.byref(cnt))
+        out[buf.value.decode()] = (ms.value, cnt.value)
+    return out
 
 
 class DeerError(RuntimeError):

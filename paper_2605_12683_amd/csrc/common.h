@@ -27,6 +27,24 @@ int hip_fail(hipError_t e, const char *what);
         if (_e != hipSuccess) return ::deer::hip_fail(_e, what);       \
     } while (0)
 
+// ---- optional per-kernel timing (HIP events on the launching stream) ----------------------
+// Off unless deer_timing_enable(1) was called; then every launch site brackets its kernel
+// with two events taken from a pool.
+bool timing_on();
+void timing_mark(const char *name, hipStream_t st, bool start);
+
+struct KTimer {
+    const char *name;
+    hipStream_t st;
+    bool on;
+    KTimer(const char *n, hipStream_t s) : name(n), st(s), on(timing_on()) {
+        if (on) timing_mark(name, st, true);
+    }
+    ~KTimer() {
+        if (on) timing_mark(name, st, false);
+    }
+};
+
 // ---- device helpers ---------------------------------------------------------------------
 
 // 16x16x4 fp32 MFMA: acc[16x16] += A[16x4] * B[4x16].  Lane l = 16*g + c holds

@@ -6,6 +6,9 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <map>
+#include <mutex>
+#include <string>
 #include <vector>
 
 #include "common.h"
@@ -25,6 +28,63 @@ void set_error(const char *fmt, ...) {
 int hip_fail(hipError_t e, const char *what) {
     set_error("%s failed: %s", what, hipGetErrorString(e));
     return DEER_ERR_HIP;
+}
+
+// ---- optional per-kernel timing ------------------------------------------------------------
+namespace {
+struct TimingState {
+    std::mutex mu;
+    bool on = false;
+    std::vector<hipEvent_t> pool;
+    std::map<std::string, std::vector<std::pair<hipEvent_t, hipEvent_t>>> recs;
+    std::vector<std::string> order;
+};
+TimingState &tstate() {
+    static TimingState s;
+    return s;
+}
+thread_local std::vector<hipEvent_t> t_open;
+
+hipEvent_t take_event(TimingState &s) {
+    if (!s.pool.empty()) {
+        hipEvent_t e = s.pool.back();
+        s.pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+}  // namespace
+
+bool timing_on() {
+    TimingState &s = tstate();
+    std::lock_guard<std::mutex> g(s.mu);
+    return s.on;
+}
+
+void timing_mark(const char *name, hipStream_t st, bool start) {
+    TimingState &s = tstate();
+    std::lock_guard<std::mutex> g(s.mu);
+    hipEvent_t e = take_event(s);
+    if (!e) return;
+    (void)hipEventRecord(e, st);
+    if (start) {
+        t_open.push_back(e);
+        return;
+    }
+    if (t_open.empty()) {
+        s.pool.push_back(e);
+        return;
+    }
+    hipEvent_t e0 = t_open.back();
+    t_open.pop_back();
+    auto it = s.recs.find(name);
+    if (it == s.recs.end()) {
+        s.order.push_back(name);
+        it = s.recs.emplace(name, std::vector<std::pair<hipEvent_t, hipEvent_t>>()).first;
+    }
+    it->second.emplace_back(e0, e);
 }
 
 // ---- small utility kernels -------------------------------------------------------------
@@ -191,6 +251,42 @@ const char *deer_status_string(int s) {
 }
 
 const char *deer_last_error(void) { return g_err; }
+
+int deer_timing_enable(int on) {
+    TimingState &s = tstate();
+    std::lock_guard<std::mutex> g(s.mu);
+    for (auto &kv : s.recs)
+        for (auto &pr : kv.second) {
+            s.pool.push_back(pr.first);
+            s.pool.push_back(pr.second);
+        }
+    s.recs.clear();
+    s.order.clear();
+    s.on = on != 0;
+    return DEER_OK;
+}
+
+int deer_timing_report(int idx, char *name, int name_cap, double *ms_total, long *launches) {
+    TimingState &s = tstate();
+    std::lock_guard<std::mutex> g(s.mu);
+    const int n = (int)s.order.size();
+    if (idx < 0 || idx >= n) return n;
+    const std::string &k = s.order[idx];
+    double tot = 0.0;
+    for (auto &pr : s.recs[k]) {
+        if (hipEventSynchronize(pr.second) != hipSuccess) return -DEER_ERR_HIP;
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess) return -DEER_ERR_HIP;
+        tot += ms;
+    }
+    if (name && name_cap > 0) {
+        strncpy(name, k.c_str(), (size_t)name_cap - 1);
+        name[name_cap - 1] = 0;
+    }
+    if (ms_total) *ms_total = tot;
+    if (launches) *launches = (long)s.recs[k].size();
+    return n;
+}
 
 size_t deer_workspace_bytes(const deer_model *m, int B, int T, int op) {
     deer_forcing f{0.f, 0};

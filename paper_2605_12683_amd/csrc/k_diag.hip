@@ -217,13 +217,22 @@ int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const floa
     float *carry = (float *)((char *)ws + one);
     const int nblk = B * ntile * nq;
     const int conj_lam = rev ? 1 : 0;
-    hipLaunchKernelGGL(k_diag_chunk<false>, dim3(nblk), dim3(DNW * 64), 0, st, lam, conj_lam, b, Bc, K, u, rev ? 1 : 0,
-                       B, T, M, ntile, nq, agg, (const float *)nullptr, (float *)nullptr);
+    {
+        KTimer _kt("k_diag_chunk_reduce", st);
+        hipLaunchKernelGGL(k_diag_chunk<false>, dim3(nblk), dim3(DNW * 64), 0, st, lam, conj_lam, b, Bc, K, u, rev ? 1 : 0,
+                           B, T, M, ntile, nq, agg, (const float *)nullptr, (float *)nullptr);
+    }
     DEER_LAUNCH_CHECK("k_diag_chunk<reduce>");
-    hipLaunchKernelGGL(k_diag_carry, dim3(B * ntile * DTC), dim3(256), 0, st, lam, conj_lam, agg, carry, ntile, M, nq);
+    {
+        KTimer _kt("k_diag_carry", st);
+        hipLaunchKernelGGL(k_diag_carry, dim3(B * ntile * DTC), dim3(256), 0, st, lam, conj_lam, agg, carry, ntile, M, nq);
+    }
     DEER_LAUNCH_CHECK("k_diag_carry");
-    hipLaunchKernelGGL(k_diag_chunk<true>, dim3(nblk), dim3(DNW * 64), 0, st, lam, conj_lam, b, Bc, K, u, rev ? 1 : 0,
-                       B, T, M, ntile, nq, agg, carry, y);
+    {
+        KTimer _kt("k_diag_chunk_fixup", st);
+        hipLaunchKernelGGL(k_diag_chunk<true>, dim3(nblk), dim3(DNW * 64), 0, st, lam, conj_lam, b, Bc, K, u, rev ? 1 : 0,
+                           B, T, M, ntile, nq, agg, carry, y);
+    }
     DEER_LAUNCH_CHECK("k_diag_chunk<fixup>");
     return DEER_OK;
 }
@@ -314,12 +323,18 @@ int launch_diag_grads(int B, int T, int M, int K, const float *a, const float *h
     const int ntile = (M + DTC - 1) / DTC;
     const int nsl = (T + DGT - 1) / DGT;
     float *part = (float *)ws;
-    hipLaunchKernelGGL(k_diag_grads_partial, dim3(B * ntile * nsl), dim3(256), 0, st, a, h, x, K, B, T, M, ntile, nsl,
-                       part);
+    {
+        KTimer _kt("k_diag_grads_partial", st);
+        hipLaunchKernelGGL(k_diag_grads_partial, dim3(B * ntile * nsl), dim3(256), 0, st, a, h, x, K, B, T, M, ntile, nsl,
+                           part);
+    }
     DEER_LAUNCH_CHECK("k_diag_grads_partial");
     const int n = M * (2 + 2 * K);
-    hipLaunchKernelGGL(k_diag_grads_final, dim3((n + 255) / 256), dim3(256), 0, st, part, K, B, M, ntile, nsl, dlam,
-                       dBc);
+    {
+        KTimer _kt("k_diag_grads_final", st);
+        hipLaunchKernelGGL(k_diag_grads_final, dim3((n + 255) / 256), dim3(256), 0, st, part, K, B, M, ntile, nsl, dlam,
+                           dBc);
+    }
     DEER_LAUNCH_CHECK("k_diag_grads_final");
     return DEER_OK;
 }

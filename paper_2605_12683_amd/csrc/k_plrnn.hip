@@ -495,6 +495,7 @@ int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, 
     const int MP = padded(a.M);
     const long groups = ((long)a.B * a.T + (64 / MP) - 1) / (64 / MP);
     const int grid = (int)(groups < 16384 ? groups : 16384);
+    KTimer kt("k_resjac_plrnn", st);
 #define RJ(MPV)                                                                                                   \
     hipLaunchKernelGGL(k_resjac_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, z, \
                        F, r, J, masks, active, a.B, a.T, a.M)
@@ -510,6 +511,7 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+    KTimer kt("k_chunk_product_plrnn", st);
 #define CP(MPV, R)                                                                                                  \
     hipLaunchKernelGGL((k_chunk_product_plrnn<MPV, R>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, \
                        rhs, z, a.x, seed_scale, P, v, active, a.B, a.T, a.M, C, ncs)
@@ -525,6 +527,7 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
 
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
                  uint32_t *norm_bits, int B, int ncs, hipStream_t st) {
+    KTimer kt("k_carry", st);
 #define CA(MPV, R) \
     hipLaunchKernelGGL((k_carry<MPV, R>), dim3(B), dim3(MPV), 0, st, P, v, carry_in, active, norm_bits, ncs)
     if (!rev) {
@@ -542,6 +545,7 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+    KTimer kt("k_fixup_fwd_plrnn", st);
 #define FX(MPV)                                                                                                       \
     hipLaunchKernelGGL(k_fixup_fwd_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, carry_in, \
                        z, norm_bits, active, a.B, a.T, a.M, C, ncs)
@@ -556,6 +560,7 @@ int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+    KTimer kt("k_fixup_rev_plrnn", st);
 #define FR(MPV)                                                                                                     \
     hipLaunchKernelGGL(k_fixup_rev_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, g,       \
                        seed_scale, a.x, a.z0, z, carry_in, lam, gpart, a.B, a.T, a.M, C, ncs)
@@ -568,7 +573,10 @@ int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
 int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *dA, float *dW, float *dh,
                         hipStream_t st) {
     const int n = MP * (MP + 2);
-    hipLaunchKernelGGL(k_reduce_gpart, dim3((n + 255) / 256), dim3(256), 0, st, gpart, nchains, MP, M, dA, dW, dh);
+    {
+        KTimer _kt("k_reduce_gpart", st);
+        hipLaunchKernelGGL(k_reduce_gpart, dim3((n + 255) / 256), dim3(256), 0, st, gpart, nchains, MP, M, dA, dW, dh);
+    }
     DEER_LAUNCH_CHECK("k_reduce_gpart");
     return DEER_OK;
 }

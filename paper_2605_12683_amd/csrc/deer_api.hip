@@ -190,6 +190,65 @@ static PlrnnWs carve_plrnn(void *ws, int B, int T, int M, int op, size_t *bytes)
     return w;
 }
 
+struct DenseWs {
+    float *P, *v, *carry;
+    int C, ncs, MP;
+};
+
+static DenseWs carve_dense(void *ws, int B, int T, int M, size_t *bytes) {
+    DenseWs w{};
+    w.MP = padded_dim(M);
+    w.C = choose_chunk(B, T, w.MP);
+    w.ncs = (T + w.C - 1) / w.C;
+    const size_t nch = (size_t)B * w.ncs;
+    Carver c(ws);
+    w.P = c.take<float>(nch * w.MP * w.MP);
+    w.v = c.take<float>(nch * w.MP);
+    w.carry = c.take<float>(nch * w.MP);
+    *bytes = c.off;
+    return w;
+}
+
+struct ShWs {
+    float *r, *J, *g, *lam, *part;
+    uint32_t *masks;
+    DenseWs d;
+    uint32_t *norm_bits;
+    int *active;
+};
+
+static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, bool need_lam, size_t *bytes) {
+    ShWs w{};
+    const int LW = (L + 31) / 32;
+    Carver c(ws);
+    w.masks = c.take<uint32_t>((size_t)B * T * LW);
+    w.J = c.take<float>((size_t)B * T * M * M);
+    w.norm_bits = c.take<uint32_t>(B);
+    w.active = c.take<int>(B);
+    if (op == DEER_OP_SOLVE) {
+        w.r = c.take<float>((size_t)B * T * M);
+    } else {
+        if (need_g) w.g = c.take<float>((size_t)B * T * M);
+        if (need_lam) w.lam = c.take<float>((size_t)B * T * M);
+        int nb = 0;
+        w.part = c.take<float>(sh_grads_part_floats(M, L, &nb));
+    }
+    size_t dbytes = 0;
+    w.d = carve_dense(ws ? (char *)ws + c.off : nullptr, B, T, M, &dbytes);
+    *bytes = c.off + dbytes;
+    return w;
+}
+
+static int check_shallow_limits(const deer_model *m) {
+    const size_t cap = 64 * 1024;
+    if (sh_resjac_lds(m->M, m->L) > cap || sh_jacform_lds(m->M, m->L) > cap) {
+        set_error("shallow PLRNN with M=%d, L=%d exceeds the 64 KiB LDS tiles of this build (need M*L <= 8192 "
+                  "for M <= 32)", m->M, m->L);
+        return DEER_ERR_INVALID_ARG;
+    }
+    return DEER_OK;
+}
+
 static int check_common(const deer_model *m, const deer_forcing *f, int B, int T) {
     if (!m || !f) { set_error("model/forcing pointer is NULL"); return DEER_ERR_INVALID_ARG; }
     if (B <= 0 || T <= 0) { set_error("B and T must be positive (B=%d, T=%d)", B, T); return DEER_ERR_INVALID_ARG; }
@@ -230,6 +289,146 @@ static size_t diag_bytes(int B, int T, int M, int op) {
         if (g > a) a = g;
     }
     return a;
+}
+
+// Host-side Newton loop shared by the PLRNN kinds.  `update(active)` queues one Newton update
+// for the sequences whose device flag is set (or all, when active is null) and leaves
+// per-sequence max|Delta| bits in norm_bits.
+template <class Update>
+static int newton_loop(const deer_solve_opts *o, int B, int *dev_active, uint32_t *norm_bits, Update update,
+                       std::vector<int> &it, std::vector<float> &norm, bool &nonfinite, std::vector<int> &act,
+                       hipStream_t st) {
+    const int fixed = o->fixed_iters > 0 ? o->fixed_iters : 0;
+    const int max_iter = o->max_iter > 0 ? o->max_iter : 500;
+    int rc;
+    if ((rc = launch_fill_i32(dev_active, B, 1, st))) return rc;
+    std::vector<uint32_t> nb(B, 0);
+    const int *dact = fixed ? nullptr : dev_active;
+    for (int k = 0;; ++k) {
+        if (fixed) {
+            if (k == fixed) break;
+        } else {
+            bool any = false;
+            for (int b = 0; b < B; ++b) any |= act[b] != 0;
+            if (!any || k == max_iter) break;
+        }
+        if ((rc = update(dact))) return rc;
+        if (fixed) continue;
+        DEER_HIP(hipMemcpyAsync(nb.data(), norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+        DEER_HIP(hipStreamSynchronize(st));
+        bool changed = false;
+        for (int b = 0; b < B; ++b) {
+            if (!act[b]) continue;
+            float e;
+            memcpy(&e, &nb[b], 4);
+            it[b] += 1;
+            norm[b] = e;
+            if (!isfinite(e)) {
+                nonfinite = true;
+                act[b] = 0;
+                changed = true;
+            } else if (e < o->tol) {
+                act[b] = 0;
+                changed = true;
+            }
+        }
+        if (changed) {
+            DEER_HIP(hipMemcpyAsync(dev_active, act.data(), B * sizeof(int), hipMemcpyHostToDevice, st));
+            DEER_HIP(hipStreamSynchronize(st));
+        }
+    }
+    if (fixed) {
+        DEER_HIP(hipMemcpyAsync(nb.data(), norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+        DEER_HIP(hipStreamSynchronize(st));
+        for (int b = 0; b < B; ++b) {
+            memcpy(&norm[b], &nb[b], 4);
+            it[b] = fixed;
+            if (!isfinite(norm[b])) nonfinite = true;
+        }
+    }
+    return DEER_OK;
+}
+
+static int finish_solve(const deer_solve_opts *o, int B, const std::vector<int> &it, const std::vector<float> &norm,
+                        bool nonfinite, const std::vector<int> &act, int32_t *iters, float *final_norm) {
+    if (iters) for (int b = 0; b < B; ++b) iters[b] = it[b];
+    if (final_norm) for (int b = 0; b < B; ++b) final_norm[b] = norm[b];
+    if (nonfinite) {
+        set_error("a Newton update produced a non-finite value");
+        return DEER_ERR_NONFINITE;
+    }
+    if (o->fixed_iters <= 0) {
+        for (int b = 0; b < B; ++b)
+            if (act[b]) {
+                set_error("sequence %d not converged after %d Newton updates (last max|dz| = %g)", b, it[b], norm[b]);
+                return DEER_ERR_NOT_CONVERGED;
+            }
+    }
+    return DEER_OK;
+}
+
+static int init_guess(const deer_solve_opts *o, int B, int T, int M, int N, const float *x, float *z, hipStream_t st) {
+    if (o->init == DEER_INIT_TEACHER) return launch_fill_teacher(B, T, M, N, x, z, st);
+    if (o->init == DEER_INIT_ZERO) return launch_fill_f32(z, (size_t)B * T * M, 0.f, st);
+    return DEER_OK;
+}
+
+static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
+                       const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
+                       void *ws, size_t ws_bytes, hipStream_t st) {
+    size_t need = 0;
+    carve_plrnn(nullptr, B, T, m->M, DEER_OP_SOLVE, &need);
+    int rc = check_ws(ws, ws_bytes, need);
+    if (rc) return rc;
+    PlrnnWs w = carve_plrnn(ws, B, T, m->M, DEER_OP_SOLVE, &need);
+    PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
+    if ((rc = init_guess(o, B, T, m->M, f->n_forced, x, z, st))) return rc;
+    std::vector<int> act(B, 1), it(B, 0);
+    std::vector<float> norm(B, NAN);
+    bool nonfinite = false;
+    auto update = [&](const int *dact) -> int {
+        int r;
+        if ((r = launch_resjac_plrnn(a, z, nullptr, w.r, nullptr, w.masks, dact, st))) return r;
+        if ((r = launch_chunk_product_plrnn(a, false, w.masks, w.r, nullptr, 0.f, w.P, w.v, dact, w.C, w.ncs, st)))
+            return r;
+        if ((r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, w.norm_bits, B, w.ncs, st))) return r;
+        return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, z, w.norm_bits, dact, w.C, w.ncs, st);
+    };
+    if ((rc = newton_loop(o, B, w.active, w.norm_bits, update, it, norm, nonfinite, act, st))) return rc;
+    if (masks) {
+        if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
+    }
+    return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
+}
+
+static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
+                         const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters,
+                         float *final_norm, void *ws, size_t ws_bytes, hipStream_t st) {
+    int rc = check_shallow_limits(m);
+    if (rc) return rc;
+    size_t need = 0;
+    carve_sh(nullptr, B, T, m->M, m->L, DEER_OP_SOLVE, false, false, &need);
+    if ((rc = check_ws(ws, ws_bytes, need))) return rc;
+    ShWs w = carve_sh(ws, B, T, m->M, m->L, DEER_OP_SOLVE, false, false, &need);
+    ShArgs a{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
+    if ((rc = init_guess(o, B, T, m->M, f->n_forced, x, z, st))) return rc;
+    std::vector<int> act(B, 1), it(B, 0);
+    std::vector<float> norm(B, NAN);
+    bool nonfinite = false;
+    const DenseWs &d = w.d;
+    auto update = [&](const int *dact) -> int {
+        int r;
+        if ((r = launch_resjac_shplrnn(a, z, nullptr, w.r, w.masks, dact, st))) return r;
+        if ((r = launch_jacform_shplrnn(a, w.masks, w.J, dact, st))) return r;
+        if ((r = launch_chunk_product_dense(false, B, T, m->M, w.J, w.r, -1.f, d.P, d.v, dact, d.C, d.ncs, st))) return r;
+        if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, w.norm_bits, B, d.ncs, st))) return r;
+        return launch_fixup_dense(0, B, T, m->M, w.J, w.r, -1.f, d.carry, z, w.norm_bits, dact, d.C, d.ncs, st);
+    };
+    if ((rc = newton_loop(o, B, w.active, w.norm_bits, update, it, norm, nonfinite, act, st))) return rc;
+    if (masks) {
+        if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, masks, nullptr, st))) return rc;
+    }
+    return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
 }
 
 }  // namespace deer
@@ -298,12 +497,22 @@ size_t deer_workspace_bytes(const deer_model *m, int B, int T, int op) {
         carve_plrnn(nullptr, B, T, m->M, op, &bytes);
         return bytes;
     }
+    if (m->kind == DEER_SHPLRNN) {
+        size_t bytes = 0;
+        carve_sh(nullptr, B, T, m->M, m->L, op, true, true, &bytes);
+        return bytes;
+    }
     return 0;
 }
 
 size_t deer_scan_workspace_bytes(int layout, int B, int T, int M) {
     if (B <= 0 || T <= 0 || M <= 0) return 0;
     if (layout == DEER_SCAN_DIAG_C64) return diag_scan_ws_bytes(B, T, M);
+    if (layout == DEER_SCAN_DENSE && M <= 64) {
+        size_t bytes = 0;
+        carve_dense(nullptr, B, T, M, &bytes);
+        return bytes;
+    }
     return 0;
 }
 
@@ -318,95 +527,18 @@ int plrnn_jacobian(const deer_model *m, const deer_forcing *f, int B, int T, con
         PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
         return launch_resjac_plrnn(a, z, F, r, J, masks, nullptr, st);
     }
+    if (m->kind == DEER_SHPLRNN) {
+        if ((rc = check_shallow_limits(m))) return rc;
+        ShArgs a{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
+        if ((rc = launch_resjac_shplrnn(a, z, F, r, masks, nullptr, st))) return rc;
+        if (J) {
+            if (!masks) { set_error("the shallow dense Jacobian output needs the masks output"); return DEER_ERR_INVALID_ARG; }
+            if ((rc = launch_jacform_shplrnn(a, masks, J, nullptr, st))) return rc;
+        }
+        return DEER_OK;
+    }
     set_error("plrnn_jacobian: model kind %d not supported", m->kind);
     return DEER_ERR_INVALID_ARG;
-}
-
-static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
-                       const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
-                       void *ws, size_t ws_bytes, hipStream_t st) {
-    size_t need = 0;
-    carve_plrnn(nullptr, B, T, m->M, DEER_OP_SOLVE, &need);
-    int rc = check_ws(ws, ws_bytes, need);
-    if (rc) return rc;
-    PlrnnWs w = carve_plrnn(ws, B, T, m->M, DEER_OP_SOLVE, &need);
-    PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
-    const int fixed = o->fixed_iters > 0 ? o->fixed_iters : 0;
-    const int max_iter = o->max_iter > 0 ? o->max_iter : 500;
-    if (o->init == DEER_INIT_TEACHER) {
-        if ((rc = launch_fill_teacher(B, T, m->M, f->n_forced, x, z, st))) return rc;
-    } else if (o->init == DEER_INIT_ZERO) {
-        if ((rc = launch_fill_f32(z, (size_t)B * T * m->M, 0.f, st))) return rc;
-    }
-    if ((rc = launch_fill_i32(w.active, B, 1, st))) return rc;
-    std::vector<int> act(B, 1), it(B, 0);
-    std::vector<uint32_t> nb(B, 0);
-    std::vector<float> norm(B, NAN);
-    bool nonfinite = false;
-    const int *dact = fixed ? nullptr : w.active;
-    for (int k = 0;; ++k) {
-        if (fixed) {
-            if (k == fixed) break;
-        } else {
-            bool any = false;
-            for (int b = 0; b < B; ++b) any |= act[b] != 0;
-            if (!any || k == max_iter) break;
-        }
-        if ((rc = launch_resjac_plrnn(a, z, nullptr, w.r, nullptr, w.masks, dact, st))) return rc;
-        if ((rc = launch_chunk_product_plrnn(a, false, w.masks, w.r, nullptr, 0.f, w.P, w.v, dact, w.C, w.ncs, st)))
-            return rc;
-        if ((rc = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, w.norm_bits, B, w.ncs, st))) return rc;
-        if ((rc = launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, z, w.norm_bits, dact, w.C, w.ncs, st))) return rc;
-        if (fixed) continue;
-        DEER_HIP(hipMemcpyAsync(nb.data(), w.norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
-        DEER_HIP(hipStreamSynchronize(st));
-        bool changed = false;
-        for (int b = 0; b < B; ++b) {
-            if (!act[b]) continue;
-            float e;
-            memcpy(&e, &nb[b], 4);
-            it[b] += 1;
-            norm[b] = e;
-            if (!isfinite(e)) {
-                nonfinite = true;
-                act[b] = 0;
-                changed = true;
-            } else if (e < o->tol) {
-                act[b] = 0;
-                changed = true;
-            }
-        }
-        if (changed) {
-            DEER_HIP(hipMemcpyAsync(w.active, act.data(), B * sizeof(int), hipMemcpyHostToDevice, st));
-            DEER_HIP(hipStreamSynchronize(st));
-        }
-    }
-    if (fixed && (iters || final_norm)) {
-        DEER_HIP(hipMemcpyAsync(nb.data(), w.norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
-        DEER_HIP(hipStreamSynchronize(st));
-        for (int b = 0; b < B; ++b) {
-            memcpy(&norm[b], &nb[b], 4);
-            it[b] = fixed;
-            if (!isfinite(norm[b])) nonfinite = true;
-        }
-    }
-    if (masks) {
-        if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
-    }
-    if (iters) for (int b = 0; b < B; ++b) iters[b] = it[b];
-    if (final_norm) for (int b = 0; b < B; ++b) final_norm[b] = norm[b];
-    if (nonfinite) {
-        set_error("a Newton update produced a non-finite value");
-        return DEER_ERR_NONFINITE;
-    }
-    if (!fixed) {
-        for (int b = 0; b < B; ++b)
-            if (act[b]) {
-                set_error("sequence %d not converged after %d Newton updates (last max|dz| = %g)", b, it[b], norm[b]);
-                return DEER_ERR_NOT_CONVERGED;
-            }
-    }
-    return DEER_OK;
 }
 
 int deer_solve(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T, const float *x,
@@ -421,6 +553,8 @@ int deer_solve(const deer_model *m, const deer_forcing *f, const deer_solve_opts
     hipStream_t st = (hipStream_t)stream;
     if (m->kind == DEER_PLRNN)
         return solve_plrnn(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
+    if (m->kind == DEER_SHPLRNN)
+        return solve_shplrnn(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
     if (m->kind == DEER_DIAG_SSM) {
         if ((rc = check_ws(ws, ws_bytes, diag_bytes(B, T, m->M, DEER_OP_SOLVE)))) return rc;
         rc = launch_diag_scan(false, B, T, m->M, m->A, nullptr, m->W, m->L, x, z, ws, st);
@@ -458,6 +592,31 @@ int deer_adjoint(const deer_model *m, const deer_forcing *f, int B, int T, const
         }
         return DEER_OK;
     }
+    if (m->kind == DEER_SHPLRNN) {
+        if ((rc = check_shallow_limits(m))) return rc;
+        size_t need = 0;
+        carve_sh(nullptr, B, T, m->M, m->L, DEER_OP_ADJOINT, true, true, &need);
+        if ((rc = check_ws(ws, ws_bytes, need))) return rc;
+        ShWs w = carve_sh(ws, B, T, m->M, m->L, DEER_OP_ADJOINT, true, true, &need);
+        ShArgs a{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
+        const DenseWs &d = w.d;
+        const float *gg = g;
+        if (!gg) {
+            const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
+            if ((rc = launch_mse_seed(z, x, scale, B, T, m->M, f->n_forced, w.g, st))) return rc;
+            gg = w.g;
+        }
+        float *lo = lam ? lam : w.lam;
+        if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, w.masks, nullptr, st))) return rc;
+        if ((rc = launch_jacform_shplrnn(a, w.masks, w.J, nullptr, st))) return rc;
+        if ((rc = launch_chunk_product_dense(true, B, T, m->M, w.J, gg, 1.f, d.P, d.v, nullptr, d.C, d.ncs, st))) return rc;
+        if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, st))) return rc;
+        if ((rc = launch_fixup_dense(2, B, T, m->M, w.J, gg, 1.f, d.carry, lo, nullptr, nullptr, d.C, d.ncs, st))) return rc;
+        if (grads && (grads->A || grads->W || grads->W2 || grads->h || grads->h2)) {
+            if ((rc = launch_grads_shplrnn(a, z, lo, w.masks, w.part, grads, st))) return rc;
+        }
+        return DEER_OK;
+    }
     if (m->kind == DEER_DIAG_SSM) {
         if (!g) { set_error("DIAG_SSM adjoint needs the cotangent g"); return DEER_ERR_INVALID_ARG; }
         if ((rc = check_ws(ws, ws_bytes, diag_bytes(B, T, m->M, DEER_OP_ADJOINT)))) return rc;
@@ -485,7 +644,19 @@ int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, cons
         if (rc) return rc;
         return launch_diag_scan(reverse != 0, B, T, M, J, b, nullptr, 0, nullptr, y, ws, st);
     }
-    set_error("deer_scan: layout %d not supported yet", layout);
+    if (layout == DEER_SCAN_DENSE) {
+        if (M > 64) { set_error("dense scans support M <= 64"); return DEER_ERR_INVALID_ARG; }
+        size_t need = 0;
+        carve_dense(nullptr, B, T, M, &need);
+        int rc = check_ws(ws, ws_bytes, need);
+        if (rc) return rc;
+        DenseWs w = carve_dense(ws, B, T, M, &need);
+        const bool rev = reverse != 0;
+        if ((rc = launch_chunk_product_dense(rev, B, T, M, J, b, 1.f, w.P, w.v, nullptr, w.C, w.ncs, st))) return rc;
+        if ((rc = launch_carry(w.MP, rev, w.P, w.v, w.carry, nullptr, nullptr, B, w.ncs, st))) return rc;
+        return launch_fixup_dense(rev ? 2 : 1, B, T, M, J, b, 1.f, w.carry, y, nullptr, nullptr, w.C, w.ncs, st);
+    }
+    set_error("deer_scan: unknown layout %d", layout);
     return DEER_ERR_INVALID_ARG;
 }
 

@@ -1,0 +1,247 @@
+// Chunked associative scan over affine pairs (J_t, b_t) with the Jacobians stored in HBM
+// ([B, T, M, M], row-major per step): the bare scan of deer_scan(DEER_SCAN_DENSE) and the
+// linear solve of every shallow-PLRNN Newton update (scheduled-sampling appendix, the pair
+// (A_t, b_t) and its composition; eq. GTF_DEER_update; eq. backward_recursion).
+//
+//   k_chunk_product_dense   per chunk: P_c = J_e ... J_s on the matrix cores (fp32 MFMA,
+//                           A operand = J_t streamed from HBM, B operand = the accumulator
+//                           itself, as in the vanilla kernel) and the chunk's local solution
+//                           v_c from a zero carry (VALU)
+//   k_fixup_dense           the chunk re-run from its carry: forward (Newton: z += Delta and
+//                           max|Delta|; bare scan: y written) or reverse (y_{t-1} = J_t^T y_t + b)
+// Carries across chunks use the shared k_carry kernel.
+#include "common.h"
+#include "launch.h"
+
+namespace deer {
+
+template <int MP>
+struct DGeo {
+    static constexpr int NCH = 64 / MP;
+    static constexpr int NI = MP / 16;
+    static constexpr int NS = MP / 4;
+};
+
+// J[row][col] of a step, zero outside M x M
+__device__ __forceinline__ float jload(const float *__restrict__ Jp, int M, int row, int col) {
+    return (row < M && col < M) ? Jp[row * M + col] : 0.f;
+}
+
+template <int MP, bool REV>
+__global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restrict__ J, const float *__restrict__ rhs,
+                                                            float rhs_sign, float *__restrict__ Pout,
+                                                            float *__restrict__ vout, const int *__restrict__ active,
+                                                            int B, int T, int M, int C, int ncs) {
+    using G = DGeo<MP>;
+    constexpr int NCH = G::NCH, NI = G::NI, NS = G::NS;
+    __shared__ __align__(16) float lds[64];
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int nchains = B * ncs;
+    const int chain0 = blockIdx.x * NCH;
+    int pb[NCH], plo[NCH], plen[NCH], us0[NCH], us1[NCH];
+    int maxlen = 0;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n) {
+        const int id = chain0 + n;
+        bool ok = id < nchains;
+        const int b = ok ? id / ncs : 0, cc = ok ? id % ncs : 0;
+        ok = ok && (!active || active[b]);
+        const int s0 = cc * C, s1 = min(s0 + C, T);
+        const int lo = REV ? s0 + 1 : s0;
+        const int hi = REV ? min(s1 + 1, T) : s1;
+        pb[n] = b;
+        plo[n] = lo;
+        plen[n] = ok ? max(hi - lo, 0) : 0;
+        us0[n] = s0;
+        us1[n] = ok ? s1 : s0;
+        maxlen = max(maxlen, max(plen[n], us1[n] - us0[n]));
+    }
+    v4f acc[NI][4];
+#pragma unroll
+    for (int Jt = 0; Jt < 4; ++Jt) {
+        const int n = (16 * Jt) / MP;
+        const int col = 16 * Jt + c - n * MP;
+#pragma unroll
+        for (int I = 0; I < NI; ++I)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[I][Jt][r] = (16 * I + 4 * g + r == col) ? 1.f : 0.f;
+    }
+    const int un = lane / MP, ui = lane % MP;
+    int ub = 0, ulo = 0, uhi = 0;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n)
+        if (n == un) { ub = pb[n]; ulo = us0[n]; uhi = us1[n]; }
+    float u = 0.f;
+
+    for (int t = 0; t < maxlen; ++t) {
+#pragma unroll
+        for (int Jt = 0; Jt < 4; ++Jt) {
+            const int n = (16 * Jt) / MP;
+            if (t < plen[n]) {
+                const float *Jp = J + ((size_t)pb[n] * T + plo[n] + t) * M * M;
+                float Aop[NI][NS];
+#pragma unroll
+                for (int I = 0; I < NI; ++I)
+#pragma unroll
+                    for (int j = 0; j < NS / 4; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) Aop[I][4 * j + q] = jload(Jp, M, 16 * I + c, 16 * j + 4 * g + q);
+                float Bop[NS];
+#pragma unroll
+                for (int j = 0; j < NS / 4; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) Bop[4 * j + q] = acc[j][Jt][q];
+#pragma unroll
+                for (int I = 0; I < NI; ++I) {
+                    v4f a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int s = 0; s < NS; ++s) a = mfma16x16x4(Aop[I][s], Bop[s], a);
+                    acc[I][Jt] = a;
+                }
+            }
+        }
+        // local solution of the chunk (lane = chain un, row ui)
+        const bool run = ulo + t < uhi;
+        if (!REV) {
+            const int s = ulo + t;
+            lds[lane] = u;
+            __syncthreads();
+            float y = 0.f;
+            if (run && ui < M) {
+                const float *Jr = J + (((size_t)ub * T + s) * M + ui) * M;
+                const float *l = lds + un * MP;
+                for (int k = 0; k < M; ++k) y = fmaf(Jr[k], l[k], y);
+            }
+            __syncthreads();
+            if (run && ui < M) u = fmaf(rhs_sign, rhs[((size_t)ub * T + s) * M + ui], y);
+        } else {
+            const int k = uhi - 1 - t;        // y_k = J_{k+1}^T y_{k+1} + b_k
+            lds[lane] = u;
+            __syncthreads();
+            float y = 0.f;
+            if (run && ui < M && t > 0) {
+                const float *Jc = J + ((size_t)ub * T + k + 1) * M * M + ui;
+                const float *l = lds + un * MP;
+                for (int r = 0; r < M; ++r) y = fmaf(Jc[(size_t)r * M], l[r], y);
+            }
+            __syncthreads();
+            if (run && ui < M) u = fmaf(rhs_sign, rhs[((size_t)ub * T + k) * M + ui], y);
+        }
+    }
+#pragma unroll
+    for (int Jt = 0; Jt < 4; ++Jt) {
+        const int n = (16 * Jt) / MP;
+        const int id = chain0 + n;
+        if (id < nchains && (plen[n] > 0 || us1[n] > us0[n])) {
+            const int col = 16 * Jt + c - n * MP;
+            float *P = Pout + (size_t)id * MP * MP;
+#pragma unroll
+            for (int I = 0; I < NI; ++I)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) P[(16 * I + 4 * g + r) * MP + col] = acc[I][Jt][r];
+        }
+    }
+    {
+        const int id = chain0 + un;
+        if (id < nchains) vout[(size_t)id * MP + ui] = u;
+    }
+}
+
+// MODE 0: forward Newton fix-up (z += Delta, per-sequence max |Delta|)
+// MODE 1: forward bare scan (y written)
+// MODE 2: reverse (y_k = J_{k+1}^T y_{k+1} + b_k written)
+template <int MP, int MODE>
+__global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J, const float *__restrict__ rhs,
+                                                    float rhs_sign, const float *__restrict__ carry_in,
+                                                    float *__restrict__ out, uint32_t *__restrict__ norm_bits,
+                                                    const int *__restrict__ active, int B, int T, int M, int C,
+                                                    int ncs) {
+    using G = DGeo<MP>;
+    __shared__ __align__(16) float lds[64];
+    const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
+    const int id = blockIdx.x * G::NCH + n;
+    const bool ok0 = id < B * ncs;
+    const int b = ok0 ? id / ncs : 0, cc = ok0 ? id % ncs : 0;
+    const bool ok = ok0 && (!active || active[b]);
+    const int s0 = cc * C, s1 = ok ? min(s0 + C, T) : s0;
+    float y = (ok && i < M) ? carry_in[(size_t)id * MP + i] : 0.f;
+    uint32_t emax = 0u;
+    const int maxlen = __builtin_amdgcn_readfirstlane(C);
+    for (int t = 0; t < maxlen; ++t) {
+        const int k = MODE == 2 ? s1 - 1 - t : s0 + t;
+        const bool run = (MODE == 2 ? k >= s0 : k < s1) && i < M;
+        lds[lane] = y;
+        __syncthreads();
+        float acc = 0.f;
+        if (run) {
+            const float *l = lds + n * MP;
+            if (MODE != 2) {
+                const float *Jr = J + (((size_t)b * T + k) * M + i) * M;
+                for (int q = 0; q < M; ++q) acc = fmaf(Jr[q], l[q], acc);
+            } else if (k + 1 < T) {
+                const float *Jc = J + ((size_t)b * T + k + 1) * M * M + i;
+                for (int r = 0; r < M; ++r) acc = fmaf(Jc[(size_t)r * M], l[r], acc);
+            }
+        }
+        __syncthreads();
+        if (run) {
+            const size_t e = ((size_t)b * T + k) * M + i;
+            y = fmaf(rhs_sign, rhs[e], acc);
+            if (MODE == 0) {
+                out[e] = out[e] + y;
+                const uint32_t ab = abs_bits(y);
+                emax = emax > ab ? emax : ab;
+            } else {
+                out[e] = y;
+            }
+        }
+    }
+    if (MODE == 0) {
+#pragma unroll
+        for (int off = MP / 2; off > 0; off >>= 1) {
+            const uint32_t o = (uint32_t)__shfl_xor((int)emax, off, 64);
+            emax = emax > o ? emax : o;
+        }
+        if (ok && i == 0) atomicMax(norm_bits + b, emax);
+    }
+}
+
+int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
+                               float *P, float *v, const int *active, int C, int ncs, hipStream_t st) {
+    const int MP = padded_dim(M);
+    const int nch = B * ncs;
+    const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+    KTimer kt("k_chunk_product_dense", st);
+#define CPD(MPV, R)                                                                                            \
+    hipLaunchKernelGGL((k_chunk_product_dense<MPV, R>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, P, v, active, \
+                       B, T, M, C, ncs)
+    if (!rev) {
+        if (MP == 16) CPD(16, false); else if (MP == 32) CPD(32, false); else CPD(64, false);
+    } else {
+        if (MP == 16) CPD(16, true); else if (MP == 32) CPD(32, true); else CPD(64, true);
+    }
+#undef CPD
+    DEER_LAUNCH_CHECK("k_chunk_product_dense");
+    return DEER_OK;
+}
+
+int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
+                       const float *carry_in, float *out, uint32_t *norm_bits, const int *active, int C, int ncs,
+                       hipStream_t st) {
+    const int MP = padded_dim(M);
+    const int nch = B * ncs;
+    const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+    KTimer kt(mode == 2 ? "k_fixup_dense_rev" : "k_fixup_dense_fwd", st);
+#define FXD(MPV, MO)                                                                                          \
+    hipLaunchKernelGGL((k_fixup_dense<MPV, MO>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, carry_in, out, \
+                       norm_bits, active, B, T, M, C, ncs)
+#define FXD3(MO) \
+    if (MP == 16) FXD(16, MO); else if (MP == 32) FXD(32, MO); else FXD(64, MO);
+    if (mode == 0) { FXD3(0) } else if (mode == 1) { FXD3(1) } else { FXD3(2) }
+#undef FXD3
+#undef FXD
+    DEER_LAUNCH_CHECK("k_fixup_dense");
+    return DEER_OK;
+}
+
+}  // namespace deer

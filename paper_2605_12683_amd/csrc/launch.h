@@ -12,6 +12,14 @@ struct PlrnnArgs {
     int B, T, M;
 };
 
+struct ShArgs {
+    const float *A, *W1, *W2, *h1, *h2;
+    float alpha;
+    int N;
+    const float *x, *z0;
+    int B, T, M, L;
+};
+
 int padded_dim(int M);
 
 // vanilla PLRNN
@@ -28,6 +36,24 @@ int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
                            const float *carry_in, float *lam, float *gpart, int C, int ncs, hipStream_t st);
 int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *dA, float *dW, float *dh,
                         hipStream_t st);
+
+// dense stored-Jacobian scan (mode: 0 Newton fix-up, 1 bare forward scan, 2 reverse)
+int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
+                               float *P, float *v, const int *active, int C, int ncs, hipStream_t st);
+int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
+                       const float *carry_in, float *out, uint32_t *norm_bits, const int *active, int C, int ncs,
+                       hipStream_t st);
+
+// shallow PLRNN
+size_t sh_resjac_lds(int M, int L);
+size_t sh_jacform_lds(int M, int L);
+size_t sh_grads_part_floats(int M, int L, int *nblocks);
+int launch_resjac_shplrnn(const ShArgs &a, const float *z, float *F, float *r, uint32_t *masks, const int *active,
+                          hipStream_t st);
+int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, const int *active, hipStream_t st);
+int launch_grads_shplrnn(const ShArgs &a, const float *z, const float *lam, const uint32_t *masks, float *part,
+                         const deer_grads *gr, hipStream_t st);
+int launch_mse_seed(const float *z, const float *x, float scale, int B, int T, int M, int N, float *g, hipStream_t st);
 
 // diagonal complex scan
 size_t diag_scan_ws_bytes(int B, int T, int M);

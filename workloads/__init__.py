@@ -271,9 +271,16 @@ def random_plrnn_case(M: int, n_obs: int, B: int, T: int, alpha: float, seed: in
                     alpha=alpha, params=params, x=np.ascontiguousarray(x))
 
 
-def random_shplrnn_case(M: int, L: int, n_obs: int, B: int, T: int, alpha: float, seed: int) -> Workload:
+def random_shplrnn_case(M: int, L: int, n_obs: int, B: int, T: int, alpha: float, seed: int,
+                        w_norm: float | None = None, a_range=(0.5, 0.95)) -> Workload:
+    """Small shallow-PLRNN case for tests.  With w_norm, W1 is rescaled so that
+    ||W1||_2 ||W2||_2 = w_norm (max A + w_norm < 1 makes the map a contraction)."""
     rng = np.random.default_rng(seed)
-    params = shplrnn_params(M, L, rng)
+    params = shplrnn_params(M, L, rng, a_range=a_range)
+    if w_norm is not None:
+        W1 = params["W1"].astype(np.float64)
+        s = np.linalg.norm(W1, 2) * np.linalg.norm(params["W2"].astype(np.float64), 2)
+        params["W1"] = (W1 * (w_norm / s)).astype(np.float32)
     x = observed_batch("lorenz96", max(n_obs, 4), B, T, seed + 1)[:, :, :n_obs].copy()
     return Workload(name=f"shplrnn_M{M}_L{L}_N{n_obs}_T{T}_B{B}", kind="shplrnn", B=B, T=T, M=M, n_obs=n_obs,
                     alpha=alpha, params=params, x=np.ascontiguousarray(x), L=L)

@@ -48,42 +48,58 @@ def _diag_step(D, model, xd, c, ws_s, ws_a, g):
     return c.B
 
 
-def roofline_for(name, c, total_ms, launches, steps, iters_per_step):
+def kernel_work(c, steps, updates):
+    """Algorithmic work of each kernel over the timed region: {name: (bound, total work)};
+    work in flop (mfma) or bytes (hbm).  `updates` = Newton updates summed over sequences."""
+    B, T, M, N = c.B, c.T, c.M, c.n_obs
+    W = (M + 31) // 32
+    fwd = updates * T                 # (b, t) steps processed by the Newton updates
+    adj = steps * B * T               # (b, t) steps of the adjoint passes
+    prod = fwd + steps * B * (T - 1)  # chunk-product steps (the adjoint product covers 1..T-1)
+    if c.kind == "diag_ssm":
+        K = c.n_obs
+        elems = steps * B * T * M
+        return {
+            # solve launch: b formed from x on the fly (x read once per step, y written);
+            # adjoint launch: cotangent read, adjoint written
+            "k_diag_chunk_fixup": ("hbm", elems * 8 + steps * B * T * 4 * K + elems * 16),
+            "k_diag_chunk_reduce": ("hbm", steps * B * T * 4 * K + elems * 8),
+            "k_diag_grads_partial": ("hbm", elems * 16 + steps * B * T * 4 * K),
+        }
+    out = {}
+    if c.kind == "plrnn":
+        out["k_chunk_product_plrnn"] = ("mfma", prod * 2.0 * M ** 3)
+        out["k_resjac_plrnn"] = ("hbm", (fwd + adj) * (8 * M + 4 * N + 4 * W))
+        out["k_fixup_fwd_plrnn"] = ("hbm", fwd * (12 * M + 4 * W))
+        out["k_fixup_rev_plrnn"] = ("hbm", adj * (8 * M + 4 * N + 4 * W))
+    else:
+        L = c.L
+        LW = (L + 31) // 32
+        out["k_jacform_shplrnn"] = ("mfma", (fwd + adj) * 2.0 * M * M * L)
+        out["k_chunk_product_dense"] = ("mfma", prod * 2.0 * M ** 3)
+        out["k_resjac_shplrnn"] = ("hbm", (fwd + adj) * (8 * M + 4 * N + 4 * LW))
+        out["k_fixup_dense_fwd"] = ("hbm", fwd * (4 * M * M + 12 * M))
+        out["k_fixup_dense_rev"] = ("hbm", adj * (4 * M * M + 8 * M))
+    return out
+
+
+def roofline_for(name, c, total_ms, launches, steps, updates):
     """Algorithmic work of the dominant kernel over the timed region, divided by its time."""
-    B, T, M = c.B, c.T, c.M
-    if name == "k_chunk_product_plrnn":
-        # forward: every Newton update composes J~_t P for all T steps of each updated sequence;
-        # adjoint: the shifted products cover steps 1..T-1 of every sequence.  2 M^3 flop each.
-        units = steps * (iters_per_step * T + B * (T - 1))
-        work = units * 2.0 * M ** 3
-        ach = work / (total_ms * 1e-3) / 1e12
-        return {"bound": "mfma", "achieved": ach, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                "frac": ach / PEAK_FP32_MFMA_TFLOPS, "traffic": None,
-                "kernel": name, "avg_launch_ms": total_ms / launches,
-                "work_per_unit": f"{2 * M ** 3} flop per (b,t) step (2 M^3, J~_t P)",
-                "units_per_launch": units / launches}
-    if name in ("k_diag_chunk_fixup", "k_diag_chunk_reduce"):
-        # fix-up: read b (8 B) + write y (8 B) per complex element; the forward launch of the
-        # solve forms b from x on the fly (8 B written per element, 12 B of x per step)
-        per = 16.0 if name == "k_diag_chunk_fixup" else 8.0
-        units = launches * B * T * M
-        work = units * per
-        ach = work / (total_ms * 1e-3) / 1e9
-        return {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
-                "traffic": None, "kernel": name, "avg_launch_ms": total_ms / launches,
-                "work_per_unit": f"{per:g} B per complex element", "units_per_launch": units / launches}
-    if name in ("k_fixup_fwd_plrnn", "k_fixup_rev_plrnn", "k_resjac_plrnn"):
-        W = (M + 31) // 32
-        per = {"k_fixup_fwd_plrnn": 4 * W + 12 * M, "k_fixup_rev_plrnn": 4 * W + 8 * M + 4 * M,
-               "k_resjac_plrnn": 8 * M + 4 * W + 4 * M}[name]
-        units = steps * (iters_per_step * T + B * T) if name != "k_fixup_rev_plrnn" else steps * B * T
-        work = units * per
-        ach = work / (total_ms * 1e-3) / 1e9
-        return {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
-                "traffic": None, "kernel": name, "avg_launch_ms": total_ms / launches,
-                "work_per_unit": f"{per} B per (b,t) step", "units_per_launch": units / launches}
-    return {"bound": "unknown", "kernel": name, "avg_launch_ms": total_ms / launches, "achieved": None,
-            "peak": None, "unit": None, "frac": None, "traffic": None}
+    work = kernel_work(c, steps, updates)
+    base = {"kernel": name, "avg_launch_ms": total_ms / launches, "launches": launches, "traffic": None}
+    if name not in work:
+        base.update({"bound": "unknown", "achieved": None, "peak": None, "unit": None, "frac": None})
+        return base
+    bound, w = work[name]
+    if bound == "mfma":
+        ach = w / (total_ms * 1e-3) / 1e12
+        base.update({"bound": "mfma", "achieved": ach, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": ach / PEAK_FP32_MFMA_TFLOPS, "work_per_launch": w / launches})
+    else:
+        ach = w / (total_ms * 1e-3) / 1e9
+        base.update({"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": ach / PEAK_HBM_GBS, "work_per_launch": w / launches})
+    return base
 
 
 def cpu_baseline(c, budget_s=20.0):
@@ -103,10 +119,15 @@ def cpu_baseline(c, budget_s=20.0):
         dt = time.perf_counter() - t0
         value, sample = Ts / dt, f"1 of {c.B} sequences, first {Ts} of {c.T} steps, forward+read-out+reverse"
     else:
-        # The oracle is vectorised over the batch and sequential in time: about 20 us per
-        # time step per Newton update.  Keep the whole batch, shorten T to fit the budget.
+        # The oracle is vectorised over the batch and sequential in time.  Calibrate on a short
+        # prefix, then keep the whole batch and shorten T to fit the budget.
+        Tc = min(c.T, 512)
+        t0 = time.perf_counter()
+        rc = O.newton(m, c.x[:, :Tc + 1], c.alpha, c.n_obs, tol=c.tol, max_iter=c.max_iter,
+                      fixed_iters=c.fixed_iters)
+        per = (time.perf_counter() - t0) / (Tc * max(1, int(rc["iters"].max())))
         Ts = c.T
-        while Ts > 1024 and Ts * 10 * 20e-6 > budget_s:
+        while Ts > 1024 and Ts * per * 12 > budget_s:
             Ts //= 2
         xs = c.x[:, :Ts + 1]
         t0 = time.perf_counter()
@@ -151,8 +172,8 @@ def main():
         gen = torch.Generator(device=dev).manual_seed(0)
         g = torch.randn(c.B, c.T, c.M, 2, device=dev, generator=gen) * 1e-6
         step = lambda: _diag_step(D, model, xd, c, ws_s, ws_a, g)          # noqa: E731
-    elif c.kind == "plrnn":
-        model = D._Model({"kind": "plrnn", **c.params})
+    elif c.kind in ("plrnn", "shplrnn"):
+        model = D._Model({"kind": c.kind, **c.params})
         ws_s = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_SOLVE))
         ws_a = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_ADJOINT))
         step = lambda: _plrnn_step(D, model, xd, c, ws_s, ws_a)            # noqa: E731
@@ -181,7 +202,11 @@ def main():
     for k, (ms, n) in sorted(kt.items(), key=lambda kv: -kv[1][0]):
         log(f"[bench] {k:28s} {ms:10.3f} ms total  {n:6d} launches  {ms / n:9.4f} ms avg")
     dom = max(kt.items(), key=lambda kv: kv[1][0])
-    roof = roofline_for(dom[0], c, dom[1][0], dom[1][1], args.steps, iters_per_step)
+    roof = roofline_for(dom[0], c, dom[1][0], dom[1][1], args.steps, updates)
+    kernels = {k: {"ms_total": ms, "launches": n, **({"frac": r["frac"], "unit": r["unit"], "achieved": r["achieved"]}
+                                                      if (r := roofline_for(k, c, ms, n, args.steps, updates))["frac"]
+                                                      is not None else {})}
+               for k, (ms, n) in kt.items()}
 
     out = {
         "metric": "DEER timesteps/sec (B*T*Newton iters)",
@@ -201,6 +226,7 @@ def main():
                    "fixed_iters": c.fixed_iters or None, "newton_updates_per_step": iters_per_step,
                    "step": "deer_solve + deer_adjoint"},
         "roofline": roof,
+        "kernels": kernels,
     }
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")

@@ -50,7 +50,7 @@ __device__ __forceinline__ float lds_dot(const float *lds, int n, const float *r
 // ---------------------------------------------------------------------------------------
 // residual, masks, F and dense J~ at every (b, t)
 // ---------------------------------------------------------------------------------------
-template <int MP>
+template <int MP, bool DENSEJ>
 __global__ __launch_bounds__(64) void k_resjac_plrnn(const float *__restrict__ A, const float *__restrict__ W,
                                                      const float *__restrict__ h, float alpha, int N,
                                                      const float *__restrict__ x, const float *__restrict__ z0,
@@ -59,7 +59,8 @@ __global__ __launch_bounds__(64) void k_resjac_plrnn(const float *__restrict__ A
                                                      uint32_t *__restrict__ masks, const int *__restrict__ active,
                                                      int B, int T, int M) {
     using G = Geo<MP>;
-    __shared__ __align__(16) float lds[64];
+    constexpr int NG = DENSEJ ? 1 : 4;    // groups of NCH rows handled per pass (memory parallelism)
+    __shared__ __align__(16) float lds[NG][64];
     const int lane = threadIdx.x;
     const int n = lane / MP, i = lane % MP;
     float wrow[MP];
@@ -69,41 +70,64 @@ __global__ __launch_bounds__(64) void k_resjac_plrnn(const float *__restrict__ A
     const float hi = (h && i < M) ? h[i] : 0.f;
     const long total = (long)B * T;
     const long ngroups = (total + G::NCH - 1) / G::NCH;
-    for (long grp = blockIdx.x; grp < ngroups; grp += gridDim.x) {
-        const long row = grp * G::NCH + n;
-        const bool in = row < total;
-        const int b = in ? (int)(row / T) : 0, s = in ? (int)(row % T) : 0;
-        const bool act = in && i < M && (!active || active[b]);
-        const float zt = act ? forced_state(x, z0, z, b, s, i, T, M, N, alpha) : 0.f;
-        const bool pos = zt > 0.f;
-        const uint64_t bal = __ballot(pos);
-        lds[lane] = pos ? zt : 0.f;
-        __syncthreads();
-        const float F = fmaf(Ai, zt, lds_dot<MP>(lds, n, wrow)) + hi;
-        __syncthreads();
-        if (act) {
-            const size_t e = (size_t)row * M + i;
-            if (r_out) r_out[e] = z[e] - F;
-            if (F_out) F_out[e] = F;
-            if (J_out) {
-                float *Jr = J_out + ((size_t)row * M + i) * M;
+    for (long grp0 = (long)blockIdx.x * NG; grp0 < ngroups; grp0 += (long)gridDim.x * NG) {
+        float zt[NG], zc[NG];
+        bool act[NG];
+        long rowv[NG];
 #pragma unroll
-                for (int j = 0; j < MP; ++j) {
-                    if (j < M) {
-                        const float mj = (float)((bal >> (n * MP + j)) & 1ull);
-                        const float v = (j == i ? Ai : 0.f) + wrow[j] * mj;
-                        Jr[j] = v * p_of(j, N, alpha);
+        for (int q = 0; q < NG; ++q) {
+            const long row = (grp0 + q) * G::NCH + n;
+            const bool in = row < total;
+            const int b = in ? (int)(row / T) : 0, s = in ? (int)(row % T) : 0;
+            act[q] = in && i < M && (!active || active[b]);
+            rowv[q] = row;
+            zt[q] = act[q] ? forced_state(x, z0, z, b, s, i, T, M, N, alpha) : 0.f;
+            zc[q] = (act[q] && r_out) ? z[(size_t)row * M + i] : 0.f;
+        }
+        uint64_t bal[NG];
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            const bool pos = zt[q] > 0.f;
+            bal[q] = __ballot(pos);
+            lds[q][lane] = pos ? zt[q] : 0.f;
+        }
+        __syncthreads();
+        float F[NG];
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            F[q] = fmaf(Ai, zt[q], lds_dot<MP>(lds[q], n, wrow)) + hi;
+            __builtin_amdgcn_sched_barrier(0);   // one dot product at a time: keeps the LDS reads of
+                                                 // the other groups from being hoisted into registers
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            const long row = rowv[q];
+            if (act[q]) {
+                const size_t e = (size_t)row * M + i;
+                if (r_out) r_out[e] = zc[q] - F[q];
+                if (F_out) F_out[e] = F[q];
+                if (DENSEJ) {
+                    float *Jr = J_out + ((size_t)row * M + i) * M;
+#pragma unroll
+                    for (int j = 0; j < MP; ++j) {
+                        if (j < M) {
+                            const float mj = (float)((bal[q] >> (n * MP + j)) & 1ull);
+                            const float v = (j == i ? Ai : 0.f) + wrow[j] * mj;
+                            Jr[j] = v * p_of(j, N, alpha);
+                        }
                     }
                 }
             }
-        }
-        if (masks && in && i == 0 && (!active || active[b])) {
-            if (MP == 64) {
-                masks[(size_t)row * 2 + 0] = (uint32_t)bal;
-                if (M > 32) masks[(size_t)row * 2 + 1] = (uint32_t)(bal >> 32);
-            } else {
-                const uint64_t seg = bal >> (n * MP);
-                masks[row] = (uint32_t)(MP == 32 ? seg : (seg & 0xffffull));
+            const bool in = row < total;
+            if (masks && in && i == 0 && (!active || active[row / T])) {
+                if (MP == 64) {
+                    masks[(size_t)row * 2 + 0] = (uint32_t)bal[q];
+                    if (M > 32) masks[(size_t)row * 2 + 1] = (uint32_t)(bal[q] >> 32);
+                } else {
+                    const uint64_t seg = bal[q] >> (n * MP);
+                    masks[row] = (uint32_t)(MP == 32 ? seg : (seg & 0xffffull));
+                }
             }
         }
     }
@@ -494,12 +518,17 @@ int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, 
                         const int *active, hipStream_t st) {
     const int MP = padded(a.M);
     const long groups = ((long)a.B * a.T + (64 / MP) - 1) / (64 / MP);
-    const int grid = (int)(groups < 16384 ? groups : 16384);
+    const long passes = J ? groups : (groups + 3) / 4;
+    const int grid = (int)(passes < 8192 ? passes : 8192);
     KTimer kt("k_resjac_plrnn", st);
-#define RJ(MPV)                                                                                                   \
-    hipLaunchKernelGGL(k_resjac_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, z, \
-                       F, r, J, masks, active, a.B, a.T, a.M)
-    if (MP == 16) RJ(16); else if (MP == 32) RJ(32); else RJ(64);
+#define RJ(MPV, DJ)                                                                                                 \
+    hipLaunchKernelGGL((k_resjac_plrnn<MPV, DJ>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, \
+                       z, F, r, J, masks, active, a.B, a.T, a.M)
+    if (J) {
+        if (MP == 16) RJ(16, true); else if (MP == 32) RJ(32, true); else RJ(64, true);
+    } else {
+        if (MP == 16) RJ(16, false); else if (MP == 32) RJ(32, false); else RJ(64, false);
+    }
 #undef RJ
     DEER_LAUNCH_CHECK("k_resjac_plrnn");
     return DEER_OK;

@@ -23,15 +23,17 @@ __device__ __forceinline__ float p_at(int i, int N, float alpha) { return i < N 
 // ---------------------------------------------------------------------------------------
 constexpr int SH_TT = 16;
 
+template <int MP>
 __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const float *__restrict__ z,
                                                         float *__restrict__ F_out, float *__restrict__ r_out,
                                                         uint32_t *__restrict__ masks, const int *__restrict__ active) {
     extern __shared__ __align__(16) float smem[];
     const int M = a.M, L = a.L, T = a.T;
-    float *zt = smem;
-    float *ru = zt + SH_TT * M;
-    float *w1t = ru + SH_TT * L;
+    float *zt = smem;                    // [SH_TT][MP], zero padded
+    float *ru = zt + SH_TT * MP;         // [SH_TT][L]
+    float *w1t = ru + SH_TT * L;         // [L][M]
     const int tid = threadIdx.x;
+    const int lane = tid & 63;
     const int LW = (L + 31) / 32;
     for (int e = tid; e < L * M; e += 256) {
         const int l = e / M, i = e % M;
@@ -42,39 +44,45 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
     for (long tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const long row0 = tile * SH_TT;
         __syncthreads();
-        for (int e = tid; e < SH_TT * M; e += 256) {
-            const int tt = e / M, i = e % M;
+        for (int e = tid; e < SH_TT * MP; e += 256) {
+            const int tt = e / MP, i = e % MP;
             const long row = row0 + tt;
             float v = 0.f;
-            if (row < total) {
+            if (row < total && i < M) {
                 const int b = (int)(row / T), s = (int)(row % T);
                 v = forced_state(a.x, a.z0, z, b, s, i, T, M, a.N, a.alpha);
             }
             zt[e] = v;
         }
         __syncthreads();
-        // hidden pre-activations, fixed order, separate roundings
+        // hidden pre-activations: left to right in k from h2, separate roundings.  The zero
+        // padding adds exact zeros, so the value is the one of the unpadded sum.
         for (int jb = 0; jb < L; jb += 256) {
             const int j = jb + tid;
             const bool jok = j < L;
+            float w2r[MP];
+#pragma unroll
+            for (int k = 0; k < MP; ++k) w2r[k] = (jok && k < M) ? a.W2[(size_t)j * M + k] : 0.f;
             const float h2j = (jok && a.h2) ? a.h2[j] : 0.f;
-            for (int tt = 0; tt < SH_TT; ++tt) {
-                float u = h2j;
-                if (jok) {
-                    const float *w2 = a.W2 + (size_t)j * M;
-                    const float *zr = zt + tt * M;
-                    for (int k = 0; k < M; ++k) u = __fadd_rn(u, __fmul_rn(w2[k], zr[k]));
-                }
-                const bool pos = jok && u > 0.f;
-                if (jok) ru[tt * L + j] = pos ? u : 0.f;
-                const uint64_t bal = __ballot(pos);
-                const long row = row0 + tt;
-                const int lane = tid & 63;
-                if (masks && row < total && (lane == 0 || lane == 32)) {
-                    const int b = (int)(row / T);
-                    if (!active || active[b]) {
-                        const int word = (jb + (tid - lane) + lane) / 32;
-                        if (word < LW) masks[(size_t)row * LW + word] = (uint32_t)(bal >> lane);
+            for (int tt0 = 0; tt0 < SH_TT; tt0 += 4) {
+                float u[4] = {h2j, h2j, h2j, h2j};
+#pragma unroll
+                for (int k = 0; k < MP; ++k)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) u[q] = __fadd_rn(u[q], __fmul_rn(w2r[k], zt[(tt0 + q) * MP + k]));
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int tt = tt0 + q;
+                    const bool pos = jok && u[q] > 0.f;
+                    if (jok) ru[tt * L + j] = pos ? u[q] : 0.f;
+                    const uint64_t bal = __ballot(pos);
+                    const long row = row0 + tt;
+                    if (masks && row < total && (lane == 0 || lane == 32)) {
+                        const int b = (int)(row / T);
+                        if (!active || active[b]) {
+                            const int word = (jb + tid) / 32;
+                            if (word < LW) masks[(size_t)row * LW + word] = (uint32_t)(bal >> lane);
+                        }
                     }
                 }
             }
@@ -95,7 +103,7 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
                 acc1 = fmaf(w1t[(l + 1) * M + i], rr[l + 1], acc1);
             }
             if (l < L) acc0 = fmaf(w1t[l * M + i], rr[l], acc0);
-            const float ztv = zt[tt * M + i];
+            const float ztv = zt[tt * MP + i];
             const float F = fmaf(a.A[i], ztv, acc0 + acc1) + (a.h1 ? a.h1[i] : 0.f);
             const size_t e2 = (size_t)row * M + i;
             if (F_out) F_out[e2] = F;
@@ -206,18 +214,20 @@ __global__ __launch_bounds__(256) void k_jacform_shplrnn(const ShArgs a, const u
 // Partials per block: [M*L (dW1, row-major) | L*M (dW2) | L (dh2) | M (dA) | M (dh1)].
 // ---------------------------------------------------------------------------------------
 constexpr int SHG_TT = 32;
+constexpr int SHG_THREADS = 256;
 
 template <int MP>
-__global__ __launch_bounds__(1024) void k_grads_shplrnn(const ShArgs a, const float *__restrict__ z,
-                                                        const float *__restrict__ lam,
-                                                        const uint32_t *__restrict__ masks,
-                                                        float *__restrict__ part) {
+__global__ __launch_bounds__(SHG_THREADS) void k_grads_shplrnn(const ShArgs a, const float *__restrict__ z,
+                                                               const float *__restrict__ lam,
+                                                               const uint32_t *__restrict__ masks,
+                                                               float *__restrict__ part) {
     __shared__ __align__(16) float zt[SHG_TT][MP];
     __shared__ __align__(16) float lm[SHG_TT][MP];
     const int M = a.M, L = a.L, T = a.T;
     const int tid = threadIdx.x;
-    const int l = tid;
+    const int l = blockIdx.y * SHG_THREADS + tid;     // hidden unit owned by this thread
     const bool lok = l < L;
+    const bool own_latent = blockIdx.y == 0 && tid < M;
     const int LW = (L + 31) / 32;
     float w2r[MP], w1c[MP], dW1c[MP], dW2r[MP];
 #pragma unroll
@@ -234,7 +244,7 @@ __global__ __launch_bounds__(1024) void k_grads_shplrnn(const ShArgs a, const fl
     for (long tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const long row0 = tile * SHG_TT;
         __syncthreads();
-        for (int e = tid; e < SHG_TT * MP; e += blockDim.x) {
+        for (int e = tid; e < SHG_TT * MP; e += SHG_THREADS) {
             const int tt = e / MP, i = e % MP;
             const long row = row0 + tt;
             float vz = 0.f, vl = 0.f;
@@ -247,7 +257,7 @@ __global__ __launch_bounds__(1024) void k_grads_shplrnn(const ShArgs a, const fl
             lm[tt][i] = vl;
         }
         __syncthreads();
-        if (tid < M) {
+        if (own_latent) {
             for (int tt = 0; tt < SHG_TT; ++tt) {
                 dA = fmaf(lm[tt][tid], zt[tt][tid], dA);
                 dh1 += lm[tt][tid];
@@ -286,7 +296,7 @@ __global__ __launch_bounds__(1024) void k_grads_shplrnn(const ShArgs a, const fl
             }
         pp[(size_t)2 * M * L + l] = dh2;
     }
-    if (tid < M) {
+    if (own_latent) {
         pp[(size_t)2 * M * L + L + tid] = dA;
         pp[(size_t)2 * M * L + L + M + tid] = dh1;
     }
@@ -335,7 +345,7 @@ __global__ void k_mse_seed(const float *__restrict__ z, const float *__restrict_
 // ---------------------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------------------
-size_t sh_resjac_lds(int M, int L) { return (size_t)(SH_TT * M + SH_TT * L + L * M) * sizeof(float); }
+size_t sh_resjac_lds(int M, int L) { return (size_t)(SH_TT * padded_dim(M) + SH_TT * L + L * M) * sizeof(float); }
 
 static int sh_LP(int L) { return (L + 15) / 16 * 16; }
 
@@ -347,7 +357,10 @@ int launch_resjac_shplrnn(const ShArgs &a, const float *z, float *F, float *r, u
     const int grid = (int)(ntiles < 4096 ? ntiles : 4096);
     const size_t lds = sh_resjac_lds(a.M, a.L);
     KTimer kt("k_resjac_shplrnn", st);
-    hipLaunchKernelGGL(k_resjac_shplrnn, dim3(grid), dim3(256), lds, st, a, z, F, r, masks, active);
+    const int MP = padded_dim(a.M);
+    if (MP == 16) hipLaunchKernelGGL(k_resjac_shplrnn<16>, dim3(grid), dim3(256), lds, st, a, z, F, r, masks, active);
+    else if (MP == 32) hipLaunchKernelGGL(k_resjac_shplrnn<32>, dim3(grid), dim3(256), lds, st, a, z, F, r, masks, active);
+    else hipLaunchKernelGGL(k_resjac_shplrnn<64>, dim3(grid), dim3(256), lds, st, a, z, F, r, masks, active);
     DEER_LAUNCH_CHECK("k_resjac_shplrnn");
     return DEER_OK;
 }
@@ -372,7 +385,7 @@ int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, con
 }
 
 size_t sh_grads_part_floats(int M, int L, int *nblocks) {
-    *nblocks = 1024;
+    *nblocks = 512;
     return (size_t)(*nblocks) * ((size_t)2 * M * L + L + 2 * M);
 }
 
@@ -381,12 +394,12 @@ int launch_grads_shplrnn(const ShArgs &a, const float *z, const float *lam, cons
     int nb = 0;
     sh_grads_part_floats(a.M, a.L, &nb);
     const int MP = padded_dim(a.M);
-    const int threads = (a.L + 63) / 64 * 64;
+    const dim3 grid(nb, (a.L + SHG_THREADS - 1) / SHG_THREADS);
     {
         KTimer kt("k_grads_shplrnn", st);
-        if (MP == 16) hipLaunchKernelGGL(k_grads_shplrnn<16>, dim3(nb), dim3(threads), 0, st, a, z, lam, masks, part);
-        else if (MP == 32) hipLaunchKernelGGL(k_grads_shplrnn<32>, dim3(nb), dim3(threads), 0, st, a, z, lam, masks, part);
-        else hipLaunchKernelGGL(k_grads_shplrnn<64>, dim3(nb), dim3(threads), 0, st, a, z, lam, masks, part);
+        if (MP == 16) hipLaunchKernelGGL(k_grads_shplrnn<16>, grid, dim3(SHG_THREADS), 0, st, a, z, lam, masks, part);
+        else if (MP == 32) hipLaunchKernelGGL(k_grads_shplrnn<32>, grid, dim3(SHG_THREADS), 0, st, a, z, lam, masks, part);
+        else hipLaunchKernelGGL(k_grads_shplrnn<64>, grid, dim3(SHG_THREADS), 0, st, a, z, lam, masks, part);
         DEER_LAUNCH_CHECK("k_grads_shplrnn");
     }
     const int width = 2 * a.M * a.L + a.L + 2 * a.M;

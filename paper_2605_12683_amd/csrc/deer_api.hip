@@ -388,9 +388,7 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     bool nonfinite = false;
     auto update = [&](const int *dact) -> int {
         int r;
-        if ((r = launch_resjac_plrnn(a, z, nullptr, w.r, nullptr, w.masks, dact, st))) return r;
-        if ((r = launch_chunk_product_plrnn(a, false, w.masks, w.r, nullptr, 0.f, w.P, w.v, dact, w.C, w.ncs, st)))
-            return r;
+        if ((r = launch_newton_product_plrnn(a, z, w.r, w.masks, w.P, w.v, dact, w.C, w.ncs, st))) return r;
         if ((r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, w.norm_bits, B, w.ncs, st))) return r;
         return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, z, w.norm_bits, dact, w.C, w.ncs, st);
     };

@@ -306,6 +306,179 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn(
 }
 
 // ---------------------------------------------------------------------------------------
+// Forward Newton pass with the residual fused in: per step of every chain the wave forms
+// z~_t, its ReLU ballot (which is at once the mask of the matrix-core bit select), F,
+// r_t = z_t - F, and advances both the chunk product and the chunk-local solution.
+// r and the masks are written for the fix-up pass.  Same MFMA layout as above.
+// ---------------------------------------------------------------------------------------
+template <int MP>
+__global__ __launch_bounds__(64) void k_newton_product_plrnn(
+    const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
+    const float *__restrict__ x, const float *__restrict__ z0, const float *__restrict__ z,
+    float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout, float *__restrict__ vout,
+    const int *__restrict__ active, int B, int T, int M, int C, int ncs) {
+    using G = Geo<MP>;
+    constexpr int NCH = G::NCH, NI = G::NI, NS = G::NS, MW = G::MW;
+    __shared__ __align__(16) float lds[64];
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int nchains = B * ncs;
+    const int chain0 = blockIdx.x * NCH;
+    int plen[NCH];
+    int maxlen = 0;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n) {
+        const int id = chain0 + n;
+        bool ok = id < nchains;
+        const int b = ok ? id / ncs : 0, cc = ok ? id % ncs : 0;
+        ok = ok && (!active || active[b]);
+        const int s0 = cc * C;
+        plen[n] = ok ? min(C, T - s0) : 0;
+        maxlen = max(maxlen, plen[n]);
+    }
+    float Aop[NI][NS];
+#pragma unroll
+    for (int I = 0; I < NI; ++I)
+#pragma unroll
+        for (int j = 0; j < NS / 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int row = 16 * I + c, col = 16 * j + 4 * g + q;
+                Aop[I][4 * j + q] = (row < M && col < M) ? W[row * M + col] * p_of(col, N, alpha) : 0.f;
+            }
+    float dI[NI][4];
+#pragma unroll
+    for (int I = 0; I < NI; ++I)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * I + 4 * g + r;
+            dI[I][r] = row < M ? A[row] * p_of(row, N, alpha) : 0.f;
+        }
+    v4f acc[NI][4];
+#pragma unroll
+    for (int Jt = 0; Jt < 4; ++Jt) {
+        const int n = (16 * Jt) / MP;
+        const int col = 16 * Jt + c - n * MP;
+#pragma unroll
+        for (int I = 0; I < NI; ++I)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[I][Jt][r] = (16 * I + 4 * g + r == col) ? 1.f : 0.f;
+    }
+    // lane-per-row part: lane = (chain un, latent ui)
+    const int un = lane / MP, ui = lane % MP;
+    const int uid = chain0 + un;
+    const bool uok0 = uid < nchains;
+    const int ub = uok0 ? uid / ncs : 0, us0 = uok0 ? (uid % ncs) * C : 0;
+    int ulen = 0;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n)
+        if (n == un) ulen = plen[n];
+    const bool lat = ui < M;
+    float wrow[MP];
+#pragma unroll
+    for (int k = 0; k < MP; ++k) wrow[k] = (lat && k < M) ? W[ui * M + k] : 0.f;
+    const float Ai = lat ? A[ui] : 0.f, hi = (lat && h) ? h[ui] : 0.f;
+    const float pi = p_of(ui, N, alpha), di = Ai * pi;
+    const bool forced = ui < N;
+    // z_{s-1} for the first step of the chunk
+    float zprev = 0.f;
+    if (ulen > 0 && lat) {
+        if (us0 == 0) zprev = z0 ? z0[(size_t)ub * M + ui] : (forced ? x[(size_t)ub * (T + 1) * N + ui] : 0.f);
+        else zprev = z[((size_t)ub * T + us0 - 1) * M + ui];
+    }
+    float u = 0.f;
+    // prefetch of step 0
+    float zcur_n = 0.f, xb_n = 0.f;
+    if (ulen > 0 && lat) {
+        zcur_n = z[((size_t)ub * T + us0) * M + ui];
+        if (forced) xb_n = x[((size_t)ub * (T + 1) + us0) * N + ui];
+    }
+    for (int t = 0; t < maxlen; ++t) {
+        const bool run = t < ulen && lat;
+        const int s = us0 + t;
+        const float zcur = zcur_n, xb = xb_n;
+        if (t + 1 < ulen && lat) {
+            zcur_n = z[((size_t)ub * T + s + 1) * M + ui];
+            if (forced) xb_n = x[((size_t)ub * (T + 1) + s + 1) * N + ui];
+        }
+        // forced state of this step (s == 0: z_0 itself)
+        float zt = 0.f;
+        if (run) {
+            if (s == 0 || !forced) zt = zprev;
+            else zt = __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xb));
+        }
+        const bool pos = zt > 0.f;
+        const uint64_t bal = __ballot(pos);
+        lds[lane] = pos ? zt : 0.f;
+        __syncthreads();
+        const float F = fmaf(Ai, zt, lds_dot<MP>(lds, un, wrow)) + hi;
+        __syncthreads();
+        const float r = zcur - F;
+        if (run) {
+            const size_t e = ((size_t)ub * T + s) * M + ui;
+            r_out[e] = r;
+            if (ui == 0) {
+                const size_t step = (size_t)ub * T + s;
+                if (MP == 64) {
+                    masks[step * 2] = (uint32_t)bal;
+                    if (M > 32) masks[step * 2 + 1] = (uint32_t)(bal >> 32);
+                } else {
+                    const uint64_t seg = bal >> (un * MP);
+                    masks[step] = (uint32_t)(MP == 32 ? seg : (seg & 0xffffull));
+                }
+            }
+        }
+        // matrix-core step of every chain still running
+#pragma unroll
+        for (int Jt = 0; Jt < 4; ++Jt) {
+            const int n = (16 * Jt) / MP;
+            if (t < plen[n]) {
+                const uint64_t seg = bal >> (n * MP);
+                const uint32_t w0 = (uint32_t)seg;
+                const uint32_t w1 = (uint32_t)(seg >> 32);
+                float Bop[NS];
+#pragma unroll
+                for (int j = 0; j < NS / 4; ++j) {
+                    const uint32_t wj = (j >> 1) ? w1 : w0;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) Bop[4 * j + q] = select_bit(wj, 16 * (j & 1) + 4 * g + q, acc[j][Jt][q]);
+                }
+#pragma unroll
+                for (int I = 0; I < NI; ++I)
+#pragma unroll
+                    for (int r2 = 0; r2 < 4; ++r2) acc[I][Jt][r2] *= dI[I][r2];
+#pragma unroll
+                for (int I = 0; I < NI; ++I)
+#pragma unroll
+                    for (int s2 = 0; s2 < NS; ++s2) acc[I][Jt] = mfma16x16x4(Aop[I][s2], Bop[s2], acc[I][Jt]);
+            }
+        }
+        // chunk-local solution: u <- d u + W (p m u) - r
+        lds[lane] = pos ? pi * u : 0.f;
+        __syncthreads();
+        const float y = fmaf(di, u, lds_dot<MP>(lds, un, wrow));
+        __syncthreads();
+        if (run) {
+            u = y - r;
+            zprev = zcur;
+        }
+    }
+#pragma unroll
+    for (int Jt = 0; Jt < 4; ++Jt) {
+        const int n = (16 * Jt) / MP;
+        const int id = chain0 + n;
+        if (id < nchains && plen[n] > 0) {
+            const int col = 16 * Jt + c - n * MP;
+            float *P = Pout + (size_t)id * MP * MP;
+#pragma unroll
+            for (int I = 0; I < NI; ++I)
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) P[(16 * I + 4 * g + r2) * MP + col] = acc[I][Jt][r2];
+        }
+    }
+    if (uok0) vout[(size_t)uid * MP + ui] = u;
+}
+
+// ---------------------------------------------------------------------------------------
 // carries across chunks (one block of MP lanes per sequence)
 //   forward: carry_in[c] = y_end(c-1),  y_end(c) = P_c y_end(c-1) + v_c
 //   reverse: carry_in[c] = lam_{s1(c)}, lam_{s0(c)} = P_c^T lam_{s1(c)} + v_c
@@ -551,6 +724,21 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
     }
 #undef CP
     DEER_LAUNCH_CHECK("k_chunk_product_plrnn");
+    return DEER_OK;
+}
+
+int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, float *r, uint32_t *masks, float *P, float *v,
+                                const int *active, int C, int ncs, hipStream_t st) {
+    const int MP = padded(a.M);
+    const int nch = a.B * ncs;
+    const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+    KTimer kt("k_newton_product_plrnn", st);
+#define NP(MPV)                                                                                                   \
+    hipLaunchKernelGGL(k_newton_product_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, \
+                       a.z0, z, r, masks, P, v, active, a.B, a.T, a.M, C, ncs)
+    if (MP == 16) NP(16); else if (MP == 32) NP(32); else NP(64);
+#undef NP
+    DEER_LAUNCH_CHECK("k_newton_product_plrnn");
     return DEER_OK;
 }
 

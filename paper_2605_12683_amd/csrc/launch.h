@@ -28,6 +28,8 @@ int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, 
 int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *masks, const float *rhs, const float *z,
                                float seed_scale, float *P, float *v, const int *active, int C, int ncs,
                                hipStream_t st);
+int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, float *r, uint32_t *masks, float *P, float *v,
+                                const int *active, int C, int ncs, hipStream_t st);
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
                  uint32_t *norm_bits, int B, int ncs, hipStream_t st);
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in, float *z,

@@ -60,16 +60,20 @@ def kernel_work(c, steps, updates):
         K = c.n_obs
         elems = steps * B * T * M
         return {
-            # solve launch: b formed from x on the fly (x read once per step, y written);
+            # single pass; solve launch: b formed from x on the fly (x read, y written);
             # adjoint launch: cotangent read, adjoint written
+            "k_diag_scan_lb": ("hbm", elems * 8 + steps * B * T * 4 * K + elems * 16),
             "k_diag_chunk_fixup": ("hbm", elems * 8 + steps * B * T * 4 * K + elems * 16),
             "k_diag_chunk_reduce": ("hbm", steps * B * T * 4 * K + elems * 8),
             "k_diag_grads_partial": ("hbm", elems * 16 + steps * B * T * 4 * K),
         }
     out = {}
     if c.kind == "plrnn":
-        out["k_chunk_product_plrnn"] = ("mfma", prod * 2.0 * M ** 3)
-        out["k_resjac_plrnn"] = ("hbm", (fwd + adj) * (8 * M + 4 * N + 4 * W))
+        # forward Newton updates run the fused kernel (residual + masks + product); the
+        # adjoint runs the shifted product and a mask pass
+        out["k_newton_product_plrnn"] = ("mfma", fwd * 2.0 * M ** 3)
+        out["k_chunk_product_plrnn"] = ("mfma", steps * B * (T - 1) * 2.0 * M ** 3)
+        out["k_resjac_plrnn"] = ("hbm", adj * (4 * M + 4 * N + 4 * W))
         out["k_fixup_fwd_plrnn"] = ("hbm", fwd * (12 * M + 4 * W))
         out["k_fixup_rev_plrnn"] = ("hbm", adj * (8 * M + 4 * N + 4 * W))
     else:

@@ -91,9 +91,11 @@ enum { DEER_INIT_TEACHER = 0, DEER_INIT_ZERO = 1, DEER_INIT_USER = 2 };
 
 typedef struct {
     float tol;          /* stop a sequence once max_{t,m} |Delta z| < tol (absolute)        */
-    int max_iter;       /* cap on Newton updates per sequence (500 if <= 0)                 */
+    int max_iter;       /* cap on Newton passes (accepted or rejected, 500 if <= 0)         */
     int fixed_iters;    /* > 0: run exactly this many updates, no convergence test/sync     */
     int init;           /* DEER_INIT_*: z^(0) = [x_{1:T}; 0], zeros, or z as passed in       */
+    float step_bound;   /* rejection threshold (see deer_solve); 0: 1e3; < 0: reject only
+                           non-finite updates                                               */
 } deer_solve_opts;
 
 /* Per-parameter gradient outputs (device, float32, NULL to skip).
@@ -120,15 +122,23 @@ size_t deer_workspace_bytes(const deer_model *model, int B, int T, int op);
  *                DEER_DIAG_SSM, z is h [B,T,M][2] (complex) and the call is the single
  *                linear scan h_t = lambda h_{t-1} + Bc x_{t-1}, h_0 = 0 (Alg. LSSM).
  *   masks        [B,T,W] out or NULL: activation masks at the returned z.
- *   iters        host [B] out or NULL: updates applied to each sequence, counting the
- *                verifying one (a sequence converged after k updates reports k).
+ *   iters        host [B] out or NULL: updates applied (accepted) to each sequence,
+ *                counting the verifying one (a sequence converged after k updates reports k).
  *   final_norm   host [B] out or NULL: max |Delta z| of each sequence's last update.
  * Each Newton update is applied before the test; a sequence whose update is below tol
  * is frozen while the others continue.  With fixed_iters == 0 the call synchronises
- * `stream` once per iteration (one device-to-host copy of B+2 words); with
- * fixed_iters > 0 it synchronises once at the end (only if iters/final_norm given).
- * Returns DEER_OK, DEER_ERR_NOT_CONVERGED (z = last iterate), DEER_ERR_NONFINITE or an
- * argument / HIP / workspace error. */
+ * `stream` once per iteration (one device-to-host copy of 2B words) and safeguards the
+ * iteration: an update that is not finite, or whose max|Delta z| exceeds
+ * step_bound * (1 + max|z|) of its sequence, is discarded and that sequence retried with
+ * the damped linearisation gamma J~ (0 <= gamma < 1; gamma = 0 is the fixed-point step
+ * z_t = F(z~_{t-1})), gamma returning to 1 (plain Newton) over accepted updates.  Every
+ * gamma has the same fixed point and the same prefix property (one more leading step exact
+ * per update), so the solution is unchanged; only the path to it differs.  With
+ * fixed_iters > 0 the updates are plain Newton steps applied unconditionally and the call
+ * synchronises once at the end (only if iters/final_norm given).
+ * Returns DEER_OK, DEER_ERR_NOT_CONVERGED (z = last accepted iterate), DEER_ERR_NONFINITE
+ * (also when the undamped fixed-point step overflows) or an argument / HIP / workspace
+ * error. */
 int deer_solve(const deer_model *model, const deer_forcing *forcing, const deer_solve_opts *opts,
                int B, int T, const float *x, const float *z0, float *z, uint32_t *masks,
                int32_t *iters, float *final_norm, void *ws, size_t ws_bytes, void *stream);

@@ -79,7 +79,7 @@ def initial_state(x: np.ndarray, M: int, z0=None) -> np.ndarray:
 def forced_states(z: np.ndarray, zbar: np.ndarray, a: np.ndarray, z0: np.ndarray) -> np.ndarray:
     """z~_{t-1} = (1 - a) z_{t-1} + a zbar_{t-1} for t >= 2 and z~_0 = z_0 (eqs. GTF,
     error_forcing; GTF-DEER residual for step 1)."""
-    zt = np.empty_like(z)
+    zt = np.zeros_like(z)
     zt[:, 0] = z0
     zt[:, 1:] = (1.0 - a) * z[:, :-1] + a * zbar[:, 1:-1]
     return zt
@@ -91,6 +91,11 @@ def forced_states(z: np.ndarray, zbar: np.ndarray, a: np.ndarray, z0: np.ndarray
 
 def _p(model, k):
     return np.asarray(model[k], f64)
+
+
+def _model64(model: dict) -> dict:
+    """The parameters promoted to float64 once (the per-step helpers then reuse them)."""
+    return {k: (v if k == "kind" or v is None else np.asarray(v, f64)) for k, v in model.items()}
 
 
 def preactivation(model: dict, zt: np.ndarray) -> np.ndarray:
@@ -132,7 +137,7 @@ def activation_mask_fp32(model: dict, z: np.ndarray, x: np.ndarray, alpha: float
     p32 = (f(1.0) - a32).astype(f)
     zbar = np.zeros((Bn, T + 1, M), f)
     zbar[:, :, :x.shape[2]] = np.asarray(x, f)
-    zt = np.empty((Bn, T, M), f)
+    zt = np.zeros((Bn, T, M), f)
     zt[:, 0] = zbar[:, 0] if z0 is None else np.asarray(z0, f)
     zt[:, 1:] = (p32 * z[:, :-1]).astype(f) + (a32 * zbar[:, 1:-1]).astype(f)
     if model["kind"] == "plrnn":
@@ -180,6 +185,7 @@ def forced_jacobians(model: dict, mask: np.ndarray, a: np.ndarray) -> np.ndarray
 def rollout(model: dict, x: np.ndarray, alpha: float, n_forced: int, z0=None) -> np.ndarray:
     """z_t = F(z~_{t-1}) for t = 1..T, one step at a time.  This is the unique
     zero-residual trajectory that DEER converges to."""
+    model = _model64(model)
     x = np.asarray(x, f64)
     Bn, T1, _ = x.shape
     T = T1 - 1
@@ -187,7 +193,7 @@ def rollout(model: dict, x: np.ndarray, alpha: float, n_forced: int, z0=None) ->
     a = forcing_weights(M, n_forced, alpha)
     zbar = teacher_states(x, M)
     zprev = initial_state(x, M, z0)
-    z = np.empty((Bn, T, M), f64)
+    z = np.zeros((Bn, T, M), f64)
     for t in range(1, T + 1):
         ztil = zprev if t == 1 else (1.0 - a) * zprev + a * zbar[:, t - 1]
         zprev = model_map(model, ztil)
@@ -203,7 +209,7 @@ def affine_recurrence(apply_J, b: np.ndarray) -> np.ndarray:
     """y_t = J_t y_{t-1} + b_t for t = 1..T with y_0 = 0 (eq. DEER_update as a linear
     recursion).  apply_J(k, v) returns J_{k+1} v for every batch row."""
     Bn, T, M = b.shape
-    out = np.empty_like(b)
+    out = np.zeros_like(b)
     prev = np.zeros((Bn, M), b.dtype)
     for k in range(T):
         prev = apply_J(k, prev) + b[:, k]
@@ -215,7 +221,7 @@ def reverse_affine_recurrence(apply_JT, g: np.ndarray) -> np.ndarray:
     """l_T = g_T and l_{t-1} = J_t^T l_t + g_{t-1} for t = T..2 (eq. backward_recursion).
     apply_JT(k, w) returns J_{k+1}^T w for every batch row."""
     Bn, T, M = g.shape
-    out = np.empty_like(g)
+    out = np.zeros_like(g)
     nxt = g[:, T - 1].copy()
     out[:, T - 1] = nxt
     for k in range(T - 2, -1, -1):      # l_{k+1} (array index k) uses J_{k+2}
@@ -230,6 +236,7 @@ def reverse_affine_recurrence(apply_JT, g: np.ndarray) -> np.ndarray:
 
 def residual_and_masks(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, z0=None):
     """r_t = z_t - F(z~_{t-1}) (eq. GTF_residual) together with F and the masks at z~."""
+    model = _model64(model)
     x = np.asarray(x, f64)
     z = np.asarray(z, f64)
     M = z.shape[2]
@@ -241,10 +248,16 @@ def residual_and_masks(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, 
 
 
 def newton(model: dict, x: np.ndarray, alpha: float, n_forced: int, *, z0=None, init: str = "teacher",
-           z_init=None, tol: float = 1e-5, max_iter: int = 500, fixed_iters: int = 0, history: bool = False):
+           z_init=None, tol: float = 1e-5, max_iter: int = 500, fixed_iters: int = 0, history: bool = False,
+           gamma: float = 1.0):
     """GTF-DEER forward solve.  Each update linearises at z^(k): Delta_t =
     J~_t Delta_{t-1} - r_t, Delta_0 = 0, solved here by the sequential recursion,
-    then z^(k+1) = z^(k) + Delta.  Returns dict(z, iters, norms, status[, history])."""
+    then z^(k+1) = z^(k) + Delta.  Returns dict(z, iters, norms, status[, history]).
+
+    gamma scales the linearisation (Delta_t = gamma J~_t Delta_{t-1} - r_t): 1 is Newton's
+    step of the algorithm, 0 the fixed-point step z_t <- F(z~_{t-1}); any gamma leaves the
+    fixed point (r = 0) unchanged.  Used to pin the safeguarded GPU iteration."""
+    model = _model64(model)
     x = np.asarray(x, f64)
     Bn, T1, _ = x.shape
     T = T1 - 1
@@ -276,7 +289,7 @@ def newton(model: dict, x: np.ndarray, alpha: float, n_forced: int, *, z0=None, 
         zt = forced_states(z, zbar, a, z0v)
         r = z - model_map(model, zt)
         mask = activation_mask(model, zt)
-        delta = affine_recurrence(lambda kk, v: jvp(model, mask[:, kk], p * v), -r)
+        delta = affine_recurrence(lambda kk, v: gamma * jvp(model, mask[:, kk], p * v), -r)
         e = np.abs(delta).reshape(Bn, -1).max(axis=1) if T > 0 else np.zeros(Bn)
         e = np.where(np.isnan(delta).reshape(Bn, -1).any(axis=1), np.nan, e)
         upd = active if fixed_iters == 0 else np.ones(Bn, bool)
@@ -341,6 +354,7 @@ def adjoint(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: i
     """lam = dL/dz by the backward recursion lam_T = g_T, lam_{t-1} = J~_t^T lam_t + g_{t-1}
     (eqs. adjoint_eq, backward_recursion with lam = -v).  J~_t is taken at z~_{t-1} of
     the given trajectory z (normally the converged one)."""
+    model = _model64(model)
     z = np.asarray(z, f64)
     M = z.shape[2]
     p = 1.0 - forcing_weights(M, n_forced, alpha)
@@ -354,20 +368,21 @@ def param_grads(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_force
                 z0=None, mask_precision: str = "float64") -> dict:
     """dL/dtheta = sum_t lam_t^T dF(z~_{t-1})/dtheta (gradients appendix, IFT summary),
     summed directly over every (b, t) in float64."""
+    model = _model64(model)
     z = np.asarray(z, f64)
     lam = np.asarray(lam, f64)
     mask, zt = _masks_at(model, x, z, alpha, n_forced, z0, mask_precision)
-    out = {"A": np.einsum("bti,bti->i", lam, zt)}
+    out = {"A": np.einsum("bti,bti->i", lam, zt, optimize=True)}
     if model["kind"] == "plrnn":
         relu = np.where(mask, zt, 0.0)
-        out["W"] = np.einsum("bti,btj->ij", lam, relu)
+        out["W"] = np.einsum("bti,btj->ij", lam, relu, optimize=True)
         out["h"] = lam.sum(axis=(0, 1))
     else:
         u = preactivation(model, zt)
         relu = np.where(mask, u, 0.0)
         delta = (lam @ _p(model, "W1")) * mask
-        out["W1"] = np.einsum("bti,btl->il", lam, relu)
-        out["W2"] = np.einsum("btl,btj->lj", delta, zt)
+        out["W1"] = np.einsum("bti,btl->il", lam, relu, optimize=True)
+        out["W2"] = np.einsum("btl,btj->lj", delta, zt, optimize=True)
         out["h1"] = lam.sum(axis=(0, 1))
         out["h2"] = delta.sum(axis=(0, 1))
     return out
@@ -398,7 +413,7 @@ def diag_scan(lam: np.ndarray, b: np.ndarray) -> np.ndarray:
     """h_t = lam * h_{t-1} + b_t, h_0 = 0, t = 1..T, complex128."""
     lam = np.asarray(lam, np.complex128)
     b = np.asarray(b, np.complex128)
-    h = np.empty_like(b)
+    h = np.zeros_like(b)
     prev = np.zeros(b.shape[:1] + b.shape[2:], np.complex128)
     for k in range(b.shape[1]):
         prev = lam * prev + b[:, k]
@@ -412,7 +427,7 @@ def diag_scan_reverse(lam: np.ndarray, g: np.ndarray) -> np.ndarray:
     multiplication by conj(lam))."""
     lam = np.asarray(lam, np.complex128)
     g = np.asarray(g, np.complex128)
-    out = np.empty_like(g)
+    out = np.zeros_like(g)
     nxt = np.zeros(g.shape[:1] + g.shape[2:], np.complex128)
     for k in range(g.shape[1] - 1, -1, -1):
         nxt = np.conj(lam) * nxt + g[:, k]
@@ -446,8 +461,8 @@ def diag_ssm_loss_and_seed(params: dict, h: np.ndarray, x: np.ndarray):
     dy = 2.0 / (Bn * No * T) * err
     ds = (dy @ Wb) * (s > 0.0)
     g = ds @ Wa
-    grads = {"Wb": np.einsum("bto,btk->ok", dy, np.maximum(s, 0.0)), "cb": dy.sum(axis=(0, 1)),
-             "Wa": np.einsum("btk,btn->kn", ds, np.real(h)), "ca": ds.sum(axis=(0, 1))}
+    grads = {"Wb": np.einsum("bto,btk->ok", dy, np.maximum(s, 0.0), optimize=True), "cb": dy.sum(axis=(0, 1)),
+             "Wa": np.einsum("btk,btn->kn", ds, np.real(h), optimize=True), "ca": ds.sum(axis=(0, 1))}
     return loss, g, grads
 
 
@@ -457,7 +472,7 @@ def diag_ssm_param_grads(a_adj: np.ndarray, h: np.ndarray, x: np.ndarray) -> dic
     hprev = np.concatenate([np.zeros_like(h[:, :1]), h[:, :-1]], axis=1)
     u = np.asarray(x, f64)[:, :-1]
     return {"lam": (a_adj * np.conj(hprev)).sum(axis=(0, 1)),
-            "Bc": np.einsum("btn,btk->nk", a_adj, u)}
+            "Bc": np.einsum("btn,btk->nk", a_adj, u, optimize=True)}
 
 
 def diag_ssm_step(params: dict, x: np.ndarray) -> dict:

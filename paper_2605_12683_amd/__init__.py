@@ -96,8 +96,10 @@ def _workspace(nbytes: int):
 
 def deer_solve(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1e-5, max_iter: int = 500,
                fixed_iters: int = 0, init: str = "teacher", z=None, want_masks: bool = False, ws=None,
-               check: bool = True) -> dict:
-    """GTF-DEER forward solve.  Returns dict(z, masks, iters, norms, status)."""
+               check: bool = True, step_bound: float = 0.0) -> dict:
+    """GTF-DEER forward solve.  Returns dict(z, masks, iters, norms, status).  step_bound:
+    threshold of the update safeguard (0: library default, < 0: only non-finite updates are
+    rejected)."""
     lib = load()
     m = _model(model)
     x = _dev(x)
@@ -118,7 +120,7 @@ def deer_solve(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1
     iters = (ctypes.c_int32 * B)()
     norms = (ctypes.c_float * B)()
     f = _b.deer_forcing(float(alpha), int(n_forced))
-    o = _b.deer_solve_opts(float(tol), int(max_iter), int(fixed_iters), _INITS[init])
+    o = _b.deer_solve_opts(float(tol), int(max_iter), int(fixed_iters), _INITS[init], float(step_bound))
     z0d = _dev(z0)
     st = lib.deer_solve(ctypes.byref(m.c), ctypes.byref(f), ctypes.byref(o), B, T, _ptr(x), _ptr(z0d), _ptr(out),
                         _ptr(masks), iters, norms, _ptr(ws), ws.numel(), _stream())

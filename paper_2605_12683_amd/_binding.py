@@ -38,7 +38,7 @@ class deer_forcing(ctypes.Structure):
 
 class deer_solve_opts(ctypes.Structure):
     _fields_ = [("tol", ctypes.c_float), ("max_iter", ctypes.c_int), ("fixed_iters", ctypes.c_int),
-                ("init", ctypes.c_int)]
+                ("init", ctypes.c_int), ("step_bound", ctypes.c_float)]
 
 
 class deer_grads(ctypes.Structure):

@@ -157,12 +157,31 @@ static int choose_chunk(int B, int T, int MP) {
     return (int)C;
 }
 
+// Per-sequence control block of the Newton loop: active flags [B] followed by the damping
+// factors gamma [B] (one host-to-device copy updates both), and 2B words of max bits
+// (max|Delta| and max|z| of the last fix-up).
+struct NewtonCtl {
+    int *active;
+    float *gamma;
+    uint32_t *norm_bits;
+    float *zalt;   // second iterate buffer [B,T,M]
+};
+
+static NewtonCtl carve_ctl(Carver &c, int B, size_t seq_elems) {
+    NewtonCtl n{};
+    uint32_t *blk = c.take<uint32_t>(2 * (size_t)B);
+    n.active = (int *)blk;
+    n.gamma = blk ? (float *)(blk + B) : nullptr;
+    n.norm_bits = c.take<uint32_t>(2 * (size_t)B);
+    n.zalt = c.take<float>((size_t)B * seq_elems);
+    return n;
+}
+
 struct PlrnnWs {
     float *r;
     uint32_t *masks;
     float *P, *v, *carry;
-    uint32_t *norm_bits;
-    int *active;
+    NewtonCtl ctl;
     float *gpart;
     int C, ncs, MP;
 };
@@ -179,9 +198,8 @@ static PlrnnWs carve_plrnn(void *ws, int B, int T, int M, int op, size_t *bytes)
     w.P = c.take<float>(nch * w.MP * w.MP);
     w.v = c.take<float>(nch * w.MP);
     w.carry = c.take<float>(nch * w.MP);
-    w.norm_bits = c.take<uint32_t>(B);
-    w.active = c.take<int>(B);
     if (op == DEER_OP_SOLVE) {
+        w.ctl = carve_ctl(c, B, (size_t)T * M);
         w.r = c.take<float>((size_t)B * T * M);
     } else {
         w.gpart = c.take<float>(nch * w.MP * (w.MP + 2));
@@ -213,8 +231,7 @@ struct ShWs {
     float *r, *J, *g, *lam, *part;
     uint32_t *masks;
     DenseWs d;
-    uint32_t *norm_bits;
-    int *active;
+    NewtonCtl ctl;
 };
 
 static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, bool need_lam, size_t *bytes) {
@@ -223,9 +240,8 @@ static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, 
     Carver c(ws);
     w.masks = c.take<uint32_t>((size_t)B * T * LW);
     w.J = c.take<float>((size_t)B * T * M * M);
-    w.norm_bits = c.take<uint32_t>(B);
-    w.active = c.take<int>(B);
     if (op == DEER_OP_SOLVE) {
+        w.ctl = carve_ctl(c, B, (size_t)T * M);
         w.r = c.take<float>((size_t)B * T * M);
     } else {
         if (need_g) w.g = c.take<float>((size_t)B * T * M);
@@ -291,61 +307,125 @@ static size_t diag_bytes(int B, int T, int M, int op) {
     return a;
 }
 
-// Host-side Newton loop shared by the PLRNN kinds.  `update(active)` queues one Newton update
-// for the sequences whose device flag is set (or all, when active is null) and leaves
-// per-sequence max|Delta| bits in norm_bits.
+// Host-side Newton loop shared by the PLRNN kinds.  `update(active, gamma, zin, zout)` queues
+// one Newton update of the sequences whose device flag is set (all, when active is null),
+// linearised with the per-sequence factor gamma (gamma J~; null: 1), reading the iterate from
+// zin and writing zin + Delta to zout (which may alias zin), and leaves per-sequence
+// max|Delta| and max|zin| bits in norm_bits[0, B) and [B, 2B).
+//
+// With a convergence test (fixed_iters == 0) every update is checked before it is kept: an
+// update that is not finite, or whose max|Delta| exceeds step_bound (1 + max|z|), is
+// rejected and the sequence retried with gamma < 1; gamma returns to 1 over accepted
+// updates.  gamma = 1 is the exact Newton step, gamma = 0 the fixed-point (Picard) step
+// z_t <- F(z~_{t-1}); every gamma keeps the fixed point, and the prefix property (an update
+// makes at least one more leading step exact) holds for every gamma.  Iterates alternate
+// between z and ctl.zalt, so a rejection costs a copy of the rejected sequences only.
+constexpr float kDefaultStepBound = 1e3f;
+constexpr float kDampFirst = 1.f / 64, kDampGrow = 4.f, kDampShrink = 4.f, kDampFloor = 1e-4f;
+
 template <class Update>
-static int newton_loop(const deer_solve_opts *o, int B, int *dev_active, uint32_t *norm_bits, Update update,
-                       std::vector<int> &it, std::vector<float> &norm, bool &nonfinite, std::vector<int> &act,
-                       hipStream_t st) {
+static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, const NewtonCtl &ctl, float *z,
+                       Update update, std::vector<int> &it, std::vector<float> &norm, bool &nonfinite,
+                       std::vector<int> &act, hipStream_t st) {
     const int fixed = o->fixed_iters > 0 ? o->fixed_iters : 0;
     const int max_iter = o->max_iter > 0 ? o->max_iter : 500;
+    const float bound = o->step_bound == 0.f ? kDefaultStepBound : o->step_bound;
+    const size_t seq_bytes = seq_elems * sizeof(float);
     int rc;
-    if ((rc = launch_fill_i32(dev_active, B, 1, st))) return rc;
-    std::vector<uint32_t> nb(B, 0);
-    const int *dact = fixed ? nullptr : dev_active;
-    for (int k = 0;; ++k) {
-        if (fixed) {
-            if (k == fixed) break;
-        } else {
-            bool any = false;
-            for (int b = 0; b < B; ++b) any |= act[b] != 0;
-            if (!any || k == max_iter) break;
-        }
-        if ((rc = update(dact))) return rc;
-        if (fixed) continue;
-        DEER_HIP(hipMemcpyAsync(nb.data(), norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
-        DEER_HIP(hipStreamSynchronize(st));
-        bool changed = false;
-        for (int b = 0; b < B; ++b) {
-            if (!act[b]) continue;
-            float e;
-            memcpy(&e, &nb[b], 4);
-            it[b] += 1;
-            norm[b] = e;
-            if (!isfinite(e)) {
-                nonfinite = true;
-                act[b] = 0;
-                changed = true;
-            } else if (e < o->tol) {
-                act[b] = 0;
-                changed = true;
-            }
-        }
-        if (changed) {
-            DEER_HIP(hipMemcpyAsync(dev_active, act.data(), B * sizeof(int), hipMemcpyHostToDevice, st));
-            DEER_HIP(hipStreamSynchronize(st));
-        }
-    }
+    std::vector<uint32_t> nb(2 * (size_t)B, 0);
     if (fixed) {
-        DEER_HIP(hipMemcpyAsync(nb.data(), norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+        for (int k = 0; k < fixed; ++k)
+            if ((rc = update(nullptr, nullptr, z, z))) return rc;
+        DEER_HIP(hipMemcpyAsync(nb.data(), ctl.norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
         DEER_HIP(hipStreamSynchronize(st));
         for (int b = 0; b < B; ++b) {
             memcpy(&norm[b], &nb[b], 4);
             it[b] = fixed;
             if (!isfinite(norm[b])) nonfinite = true;
         }
+        return DEER_OK;
     }
+    // host mirror of the control block: act [B] | gamma [B]
+    std::vector<uint32_t> hctl(2 * (size_t)B);
+    std::vector<float> om(B, 0.f);   // 1 - gamma
+    auto push_ctl = [&]() -> int {
+        for (int b = 0; b < B; ++b) {
+            hctl[b] = (uint32_t)act[b];
+            const float gm = 1.f - om[b];
+            memcpy(&hctl[B + b], &gm, 4);
+        }
+        DEER_HIP(hipMemcpyAsync(ctl.active, hctl.data(), 2 * B * sizeof(uint32_t), hipMemcpyHostToDevice, st));
+        DEER_HIP(hipStreamSynchronize(st));
+        return DEER_OK;
+    };
+    if ((rc = push_ctl())) return rc;
+    float *buf[2] = {z, ctl.zalt};
+    int cur = 0;
+    std::vector<int> holder(B, 0);   // buffer that holds each sequence's iterate
+    std::vector<int> acc, rej;
+    for (int k = 0;; ++k) {
+        bool any = false;
+        for (int b = 0; b < B; ++b) any |= act[b] != 0;
+        if (!any || k == max_iter) break;
+        if ((rc = update(ctl.active, ctl.gamma, buf[cur], buf[1 - cur]))) return rc;
+        DEER_HIP(hipMemcpyAsync(nb.data(), ctl.norm_bits, 2 * B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+        DEER_HIP(hipStreamSynchronize(st));
+        bool changed = false;
+        acc.clear();
+        rej.clear();
+        for (int b = 0; b < B; ++b) {
+            if (!act[b]) continue;
+            float e, zn;
+            memcpy(&e, &nb[b], 4);
+            memcpy(&zn, &nb[B + b], 4);
+            const bool fin = isfinite(e);
+            const bool keep = fin && (bound < 0.f || om[b] >= 1.f || e <= bound * (1.f + zn));
+            if (keep) {
+                acc.push_back(b);
+                it[b] += 1;
+                norm[b] = e;
+                if (om[b] > 0.f) {
+                    om[b] = om[b] / kDampShrink < kDampFloor ? 0.f : om[b] / kDampShrink;
+                    changed = true;
+                }
+                if (e < o->tol) {
+                    act[b] = 0;
+                    changed = true;
+                }
+            } else if (om[b] >= 1.f) {
+                // the fixed-point step itself overflows: the trajectory is not finite
+                rej.push_back(b);
+                norm[b] = e;
+                nonfinite = true;
+                act[b] = 0;
+                changed = true;
+            } else {
+                rej.push_back(b);
+                om[b] = om[b] == 0.f ? kDampFirst : (om[b] * kDampGrow > 1.f ? 1.f : om[b] * kDampGrow);
+                changed = true;
+            }
+        }
+        // keep every sequence's iterate in one buffer: copy the smaller set across
+        if (!acc.empty()) {
+            if (acc.size() >= rej.size()) {
+                for (int b : rej)
+                    DEER_HIP(hipMemcpyAsync(buf[1 - cur] + b * seq_elems, buf[cur] + b * seq_elems, seq_bytes,
+                                            hipMemcpyDeviceToDevice, st));
+                cur = 1 - cur;
+            } else {
+                for (int b : acc)
+                    DEER_HIP(hipMemcpyAsync(buf[cur] + b * seq_elems, buf[1 - cur] + b * seq_elems, seq_bytes,
+                                            hipMemcpyDeviceToDevice, st));
+            }
+        }
+        for (int b : acc) holder[b] = cur;
+        for (int b : rej) holder[b] = cur;
+        if (changed && (rc = push_ctl())) return rc;
+    }
+    for (int b = 0; b < B; ++b)
+        if (holder[b] == 1)
+            DEER_HIP(hipMemcpyAsync(z + b * seq_elems, ctl.zalt + b * seq_elems, seq_bytes, hipMemcpyDeviceToDevice,
+                                    st));
     return DEER_OK;
 }
 
@@ -386,13 +466,14 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     std::vector<int> act(B, 1), it(B, 0);
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
-    auto update = [&](const int *dact) -> int {
+    uint32_t *nbits = w.ctl.norm_bits;
+    auto update = [&](const int *dact, const float *gam, const float *zin, float *zout) -> int {
         int r;
-        if ((r = launch_newton_product_plrnn(a, z, w.r, w.masks, w.P, w.v, dact, w.C, w.ncs, st))) return r;
-        if ((r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, w.norm_bits, B, w.ncs, st))) return r;
-        return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, z, w.norm_bits, dact, w.C, w.ncs, st);
+        if ((r = launch_newton_product_plrnn(a, zin, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, st))) return r;
+        if ((r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, nbits, B, w.ncs, st))) return r;
+        return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, zin, zout, nbits, dact, gam, w.C, w.ncs, st);
     };
-    if ((rc = newton_loop(o, B, w.active, w.norm_bits, update, it, norm, nonfinite, act, st))) return rc;
+    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
         if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
     }
@@ -414,15 +495,16 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
     const DenseWs &d = w.d;
-    auto update = [&](const int *dact) -> int {
+    uint32_t *nbits = w.ctl.norm_bits;
+    auto update = [&](const int *dact, const float *gam, const float *zin, float *zout) -> int {
         int r;
-        if ((r = launch_resjac_shplrnn(a, z, nullptr, w.r, w.masks, dact, st))) return r;
-        if ((r = launch_jacform_shplrnn(a, w.masks, w.J, dact, st))) return r;
+        if ((r = launch_resjac_shplrnn(a, zin, nullptr, w.r, w.masks, dact, st))) return r;
+        if ((r = launch_jacform_shplrnn(a, w.masks, w.J, dact, gam, st))) return r;
         if ((r = launch_chunk_product_dense(false, B, T, m->M, w.J, w.r, -1.f, d.P, d.v, dact, d.C, d.ncs, st))) return r;
-        if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, w.norm_bits, B, d.ncs, st))) return r;
-        return launch_fixup_dense(0, B, T, m->M, w.J, w.r, -1.f, d.carry, z, w.norm_bits, dact, d.C, d.ncs, st);
+        if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nbits, B, d.ncs, st))) return r;
+        return launch_fixup_dense(0, B, T, m->M, w.J, w.r, -1.f, d.carry, zin, zout, nbits, dact, d.C, d.ncs, st);
     };
-    if ((rc = newton_loop(o, B, w.active, w.norm_bits, update, it, norm, nonfinite, act, st))) return rc;
+    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
         if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, masks, nullptr, st))) return rc;
     }
@@ -531,7 +613,7 @@ int plrnn_jacobian(const deer_model *m, const deer_forcing *f, int B, int T, con
         if ((rc = launch_resjac_shplrnn(a, z, F, r, masks, nullptr, st))) return rc;
         if (J) {
             if (!masks) { set_error("the shallow dense Jacobian output needs the masks output"); return DEER_ERR_INVALID_ARG; }
-            if ((rc = launch_jacform_shplrnn(a, masks, J, nullptr, st))) return rc;
+            if ((rc = launch_jacform_shplrnn(a, masks, J, nullptr, nullptr, st))) return rc;
         }
         return DEER_OK;
     }
@@ -606,10 +688,10 @@ int deer_adjoint(const deer_model *m, const deer_forcing *f, int B, int T, const
         }
         float *lo = lam ? lam : w.lam;
         if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, w.masks, nullptr, st))) return rc;
-        if ((rc = launch_jacform_shplrnn(a, w.masks, w.J, nullptr, st))) return rc;
+        if ((rc = launch_jacform_shplrnn(a, w.masks, w.J, nullptr, nullptr, st))) return rc;
         if ((rc = launch_chunk_product_dense(true, B, T, m->M, w.J, gg, 1.f, d.P, d.v, nullptr, d.C, d.ncs, st))) return rc;
         if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, st))) return rc;
-        if ((rc = launch_fixup_dense(2, B, T, m->M, w.J, gg, 1.f, d.carry, lo, nullptr, nullptr, d.C, d.ncs, st))) return rc;
+        if ((rc = launch_fixup_dense(2, B, T, m->M, w.J, gg, 1.f, d.carry, nullptr, lo, nullptr, nullptr, d.C, d.ncs, st))) return rc;
         if (grads && (grads->A || grads->W || grads->W2 || grads->h || grads->h2)) {
             if ((rc = launch_grads_shplrnn(a, z, lo, w.masks, w.part, grads, st))) return rc;
         }
@@ -652,7 +734,7 @@ int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, cons
         const bool rev = reverse != 0;
         if ((rc = launch_chunk_product_dense(rev, B, T, M, J, b, 1.f, w.P, w.v, nullptr, w.C, w.ncs, st))) return rc;
         if ((rc = launch_carry(w.MP, rev, w.P, w.v, w.carry, nullptr, nullptr, B, w.ncs, st))) return rc;
-        return launch_fixup_dense(rev ? 2 : 1, B, T, M, J, b, 1.f, w.carry, y, nullptr, nullptr, w.C, w.ncs, st);
+        return launch_fixup_dense(rev ? 2 : 1, B, T, M, J, b, 1.f, w.carry, nullptr, y, nullptr, nullptr, w.C, w.ncs, st);
     }
     set_error("deer_scan: unknown layout %d", layout);
     return DEER_ERR_INVALID_ARG;

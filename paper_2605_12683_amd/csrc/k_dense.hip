@@ -147,13 +147,14 @@ __global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restr
     }
 }
 
-// MODE 0: forward Newton fix-up (z += Delta, per-sequence max |Delta|)
+// MODE 0: forward Newton fix-up (out = zin + Delta, zin may alias out; per-sequence max |Delta|
+//         and max |zin|)
 // MODE 1: forward bare scan (y written)
 // MODE 2: reverse (y_k = J_{k+1}^T y_{k+1} + b_k written)
 template <int MP, int MODE>
 __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J, const float *__restrict__ rhs,
                                                     float rhs_sign, const float *__restrict__ carry_in,
-                                                    float *__restrict__ out, uint32_t *__restrict__ norm_bits,
+                                                    const float *zin, float *out, uint32_t *__restrict__ norm_bits,
                                                     const int *__restrict__ active, int B, int T, int M, int C,
                                                     int ncs) {
     using G = DGeo<MP>;
@@ -165,7 +166,7 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
     const bool ok = ok0 && (!active || active[b]);
     const int s0 = cc * C, s1 = ok ? min(s0 + C, T) : s0;
     float y = (ok && i < M) ? carry_in[(size_t)id * MP + i] : 0.f;
-    uint32_t emax = 0u;
+    uint32_t emax = 0u, zmax = 0u;
     const int maxlen = __builtin_amdgcn_readfirstlane(C);
     for (int t = 0; t < maxlen; ++t) {
         const int k = MODE == 2 ? s1 - 1 - t : s0 + t;
@@ -188,9 +189,11 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
             const size_t e = ((size_t)b * T + k) * M + i;
             y = fmaf(rhs_sign, rhs[e], acc);
             if (MODE == 0) {
-                out[e] = out[e] + y;
-                const uint32_t ab = abs_bits(y);
+                const float zo = zin[e];
+                out[e] = zo + y;
+                const uint32_t ab = abs_bits(y), zb = abs_bits(zo);
                 emax = emax > ab ? emax : ab;
+                zmax = zmax > zb ? zmax : zb;
             } else {
                 out[e] = y;
             }
@@ -200,9 +203,14 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
 #pragma unroll
         for (int off = MP / 2; off > 0; off >>= 1) {
             const uint32_t o = (uint32_t)__shfl_xor((int)emax, off, 64);
+            const uint32_t oz = (uint32_t)__shfl_xor((int)zmax, off, 64);
             emax = emax > o ? emax : o;
+            zmax = zmax > oz ? zmax : oz;
         }
-        if (ok && i == 0) atomicMax(norm_bits + b, emax);
+        if (ok && i == 0) {
+            atomicMax(norm_bits + b, emax);
+            atomicMax(norm_bits + B + b, zmax);
+        }
     }
 }
 
@@ -226,15 +234,15 @@ int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, co
 }
 
 int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
-                       const float *carry_in, float *out, uint32_t *norm_bits, const int *active, int C, int ncs,
-                       hipStream_t st) {
+                       const float *carry_in, const float *zin, float *out, uint32_t *norm_bits, const int *active,
+                       int C, int ncs, hipStream_t st) {
     const int MP = padded_dim(M);
     const int nch = B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt(mode == 2 ? "k_fixup_dense_rev" : "k_fixup_dense_fwd", st);
 #define FXD(MPV, MO)                                                                                          \
-    hipLaunchKernelGGL((k_fixup_dense<MPV, MO>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, carry_in, out, \
-                       norm_bits, active, B, T, M, C, ncs)
+    hipLaunchKernelGGL((k_fixup_dense<MPV, MO>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, carry_in, zin, \
+                       out, norm_bits, active, B, T, M, C, ncs)
 #define FXD3(MO) \
     if (MP == 16) FXD(16, MO); else if (MP == 32) FXD(32, MO); else FXD(64, MO);
     if (mode == 0) { FXD3(0) } else if (mode == 1) { FXD3(1) } else { FXD3(2) }

@@ -316,7 +316,7 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
     const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
     const float *__restrict__ x, const float *__restrict__ z0, const float *__restrict__ z,
     float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout, float *__restrict__ vout,
-    const int *__restrict__ active, int B, int T, int M, int C, int ncs) {
+    const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C, int ncs) {
     using G = Geo<MP>;
     constexpr int NCH = G::NCH, NI = G::NI, NS = G::NS, MW = G::MW;
     __shared__ __align__(16) float lds[64];
@@ -324,6 +324,7 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
     const int nchains = B * ncs;
     const int chain0 = blockIdx.x * NCH;
     int plen[NCH];
+    float gam[NCH];                       // damping of the linearisation (1 = exact Newton)
     int maxlen = 0;
 #pragma unroll
     for (int n = 0; n < NCH; ++n) {
@@ -333,6 +334,7 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
         ok = ok && (!active || active[b]);
         const int s0 = cc * C;
         plen[n] = ok ? min(C, T - s0) : 0;
+        gam[n] = gamma ? gamma[b] : 1.f;
         maxlen = max(maxlen, plen[n]);
     }
     float Aop[NI][NS];
@@ -353,6 +355,15 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
             const int row = 16 * I + 4 * g + r;
             dI[I][r] = row < M ? A[row] * p_of(row, N, alpha) : 0.f;
         }
+    if (NCH == 1) {   // one chain per wave: fold its damping into the operands once
+#pragma unroll
+        for (int I = 0; I < NI; ++I) {
+#pragma unroll
+            for (int s2 = 0; s2 < NS; ++s2) Aop[I][s2] *= gam[0];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dI[I][r] *= gam[0];
+        }
+    }
     v4f acc[NI][4];
 #pragma unroll
     for (int Jt = 0; Jt < 4; ++Jt) {
@@ -379,6 +390,10 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
     const float Ai = lat ? A[ui] : 0.f, hi = (lat && h) ? h[ui] : 0.f;
     const float pi = p_of(ui, N, alpha), di = Ai * pi;
     const bool forced = ui < N;
+    float ugam = 1.f;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n)
+        if (n == un) ugam = gam[n];
     // z_{s-1} for the first step of the chunk
     float zprev = 0.f;
     if (ulen > 0 && lat) {
@@ -442,6 +457,15 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
 #pragma unroll
                     for (int q = 0; q < 4; ++q) Bop[4 * j + q] = select_bit(wj, 16 * (j & 1) + 4 * g + q, acc[j][Jt][q]);
                 }
+                if (NCH > 1 && gam[n] != 1.f) {   // damped chain (uniform branch)
+                    const float gm = gam[n];
+#pragma unroll
+                    for (int s2 = 0; s2 < NS; ++s2) Bop[s2] *= gm;
+#pragma unroll
+                    for (int I = 0; I < NI; ++I)
+#pragma unroll
+                        for (int r2 = 0; r2 < 4; ++r2) acc[I][Jt][r2] *= gm;
+                }
 #pragma unroll
                 for (int I = 0; I < NI; ++I)
 #pragma unroll
@@ -452,13 +476,13 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
                     for (int s2 = 0; s2 < NS; ++s2) acc[I][Jt] = mfma16x16x4(Aop[I][s2], Bop[s2], acc[I][Jt]);
             }
         }
-        // chunk-local solution: u <- d u + W (p m u) - r
+        // chunk-local solution: u <- gamma (d u + W (p m u)) - r
         lds[lane] = pos ? pi * u : 0.f;
         __syncthreads();
         const float y = fmaf(di, u, lds_dot<MP>(lds, un, wrow));
         __syncthreads();
         if (run) {
-            u = y - r;
+            u = fmaf(ugam, y, -r);
             zprev = zcur;
         }
     }
@@ -489,7 +513,10 @@ __global__ __launch_bounds__(MP) void k_carry(const float *__restrict__ P, const
                                               uint32_t *__restrict__ norm_bits, int ncs) {
     __shared__ __align__(16) float cs[MP];
     const int b = blockIdx.x, i = threadIdx.x;
-    if (norm_bits && i == 0) norm_bits[b] = 0u;
+    if (norm_bits && i == 0) {   // [0, B): max|Delta|, [B, 2B): max|z| of the next fix-up
+        norm_bits[b] = 0u;
+        norm_bits[gridDim.x + b] = 0u;
+    }
     if (active && !active[b]) return;
     float cur = 0.f;
     float pr[MP], pn[MP];
@@ -537,8 +564,9 @@ template <int MP>
 __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict__ A, const float *__restrict__ W,
                                                         float alpha, int N, const uint32_t *__restrict__ masks,
                                                         const float *__restrict__ r, const float *__restrict__ carry_in,
-                                                        float *__restrict__ z, uint32_t *__restrict__ norm_bits,
-                                                        const int *__restrict__ active, int B, int T, int M, int C,
+                                                        const float *zin, float *zout,
+                                                        uint32_t *__restrict__ norm_bits, const int *__restrict__ active,
+                                                        const float *__restrict__ gamma, int B, int T, int M, int C,
                                                         int ncs) {
     using G = Geo<MP>;
     __shared__ __align__(16) float lds[64];
@@ -548,12 +576,13 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict_
     const int b = ok0 ? id / ncs : 0, cc = ok0 ? id % ncs : 0;
     const bool ok = ok0 && (!active || active[b]);
     const int s0 = cc * C, len = ok ? min(C, T - s0) : 0;
+    const float gm = gamma ? gamma[b] : 1.f;
     float wrow[MP];
 #pragma unroll
     for (int k = 0; k < MP; ++k) wrow[k] = (i < M && k < M) ? W[i * M + k] * p_of(k, N, alpha) : 0.f;
     const float d = i < M ? A[i] * p_of(i, N, alpha) : 0.f;
     float D = (ok && i < M) ? carry_in[(size_t)id * MP + i] : 0.f;
-    uint32_t emax = 0u;
+    uint32_t emax = 0u, zmax = 0u;
     const int maxlen = __builtin_amdgcn_readfirstlane(C);
     for (int t = 0; t < maxlen; ++t) {
         const bool run = t < len && i < M;
@@ -563,20 +592,27 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict_
         const float y = fmaf(d, D, lds_dot<MP>(lds, n, wrow));
         __syncthreads();
         if (run) {
-            D = y - r[step * M + i];
+            D = fmaf(gm, y, -r[step * M + i]);
             const size_t e = step * M + i;
-            z[e] = z[e] + D;
-            const uint32_t ab = abs_bits(D);
+            const float zo = zin[e];
+            zout[e] = zo + D;
+            const uint32_t ab = abs_bits(D), zb = abs_bits(zo);
             emax = emax > ab ? emax : ab;
+            zmax = zmax > zb ? zmax : zb;
         }
     }
     // max over the MP lanes of this chain
 #pragma unroll
     for (int off = MP / 2; off > 0; off >>= 1) {
         const uint32_t o = (uint32_t)__shfl_xor((int)emax, off, 64);
+        const uint32_t oz = (uint32_t)__shfl_xor((int)zmax, off, 64);
         emax = emax > o ? emax : o;
+        zmax = zmax > oz ? zmax : oz;
     }
-    if (ok && i == 0) atomicMax(norm_bits + b, emax);
+    if (ok && i == 0) {
+        atomicMax(norm_bits + b, emax);
+        atomicMax(norm_bits + B + b, zmax);
+    }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -728,14 +764,14 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
 }
 
 int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, float *r, uint32_t *masks, float *P, float *v,
-                                const int *active, int C, int ncs, hipStream_t st) {
+                                const int *active, const float *gamma, int C, int ncs, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt("k_newton_product_plrnn", st);
 #define NP(MPV)                                                                                                   \
     hipLaunchKernelGGL(k_newton_product_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, \
-                       a.z0, z, r, masks, P, v, active, a.B, a.T, a.M, C, ncs)
+                       a.z0, z, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs)
     if (MP == 16) NP(16); else if (MP == 32) NP(32); else NP(64);
 #undef NP
     DEER_LAUNCH_CHECK("k_newton_product_plrnn");
@@ -757,15 +793,16 @@ int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_
     return DEER_OK;
 }
 
-int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in, float *z,
-                           uint32_t *norm_bits, const int *active, int C, int ncs, hipStream_t st) {
+int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
+                           const float *zin, float *zout, uint32_t *norm_bits, const int *active, const float *gamma,
+                           int C, int ncs, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt("k_fixup_fwd_plrnn", st);
 #define FX(MPV)                                                                                                       \
     hipLaunchKernelGGL(k_fixup_fwd_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, carry_in, \
-                       z, norm_bits, active, a.B, a.T, a.M, C, ncs)
+                       zin, zout, norm_bits, active, gamma, a.B, a.T, a.M, C, ncs)
     if (MP == 16) FX(16); else if (MP == 32) FX(32); else FX(64);
 #undef FX
     DEER_LAUNCH_CHECK("k_fixup_fwd_plrnn");

@@ -121,7 +121,7 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
 template <int MP, int NT>
 __global__ __launch_bounds__(256) void k_jacform_shplrnn(const ShArgs a, const uint32_t *__restrict__ masks,
                                                          float *__restrict__ Jout, const int *__restrict__ active,
-                                                         int LP) {
+                                                         const float *__restrict__ gamma, int LP) {
     extern __shared__ __align__(16) float smem[];
     constexpr int NI = MP / 16;
     const int M = a.M, L = a.L, T = a.T, N = a.N;
@@ -194,6 +194,8 @@ __global__ __launch_bounds__(256) void k_jacform_shplrnn(const ShArgs a, const u
         for (int nt = 0; nt < NT; ++nt) {
             if (!rok[nt]) continue;
             float *Jp = Jout + (size_t)(row0 + nt) * M * M;
+            // damping of the linearisation of this sequence (1 = exact Newton)
+            const float gm = gamma ? gamma[(row0 + nt) / T] : 1.f;
 #pragma unroll
             for (int I = 0; I < NI; ++I)
 #pragma unroll
@@ -201,7 +203,8 @@ __global__ __launch_bounds__(256) void k_jacform_shplrnn(const ShArgs a, const u
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int row = 16 * I + 4 * g + r, col = 16 * Jt + c;
-                        if (row < M && col < M) Jp[row * M + col] = acc[nt][I][Jt][r] + (row == col ? dI[I][r] : 0.f);
+                        if (row < M && col < M)
+                            Jp[row * M + col] = gm * (acc[nt][I][Jt][r] + (row == col ? dI[I][r] : 0.f));
                     }
         }
     }
@@ -365,7 +368,8 @@ int launch_resjac_shplrnn(const ShArgs &a, const float *z, float *F, float *r, u
     return DEER_OK;
 }
 
-int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, const int *active, hipStream_t st) {
+int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, const int *active, const float *gamma,
+                           hipStream_t st) {
     const int MP = padded_dim(a.M);
     const int LP = sh_LP(a.L);
     const size_t lds = sh_jacform_lds(a.M, a.L);
@@ -376,7 +380,8 @@ int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, con
         const long groups = (total + NTV - 1) / NTV;                                                              \
         const long want = (groups + 3) / 4;                                                                       \
         const int grid = (int)(want < 2048 ? want : 2048);                                                        \
-        hipLaunchKernelGGL((k_jacform_shplrnn<MPV, NTV>), dim3(grid), dim3(256), lds, st, a, masks, J, active, LP); \
+        hipLaunchKernelGGL((k_jacform_shplrnn<MPV, NTV>), dim3(grid), dim3(256), lds, st, a, masks, J, active, gamma, \
+                           LP);                                                                              \
     }
     if (MP == 16) JF(16, 4) else if (MP == 32) JF(32, 4) else JF(64, 1)
 #undef JF

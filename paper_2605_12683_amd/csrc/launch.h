@@ -29,11 +29,12 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
                                float seed_scale, float *P, float *v, const int *active, int C, int ncs,
                                hipStream_t st);
 int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, float *r, uint32_t *masks, float *P, float *v,
-                                const int *active, int C, int ncs, hipStream_t st);
+                                const int *active, const float *gamma, int C, int ncs, hipStream_t st);
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
                  uint32_t *norm_bits, int B, int ncs, hipStream_t st);
-int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in, float *z,
-                           uint32_t *norm_bits, const int *active, int C, int ncs, hipStream_t st);
+int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
+                           const float *zin, float *zout, uint32_t *norm_bits, const int *active, const float *gamma,
+                           int C, int ncs, hipStream_t st);
 int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *g, float seed_scale, const float *z,
                            const float *carry_in, float *lam, float *gpart, int C, int ncs, hipStream_t st);
 int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *dA, float *dW, float *dh,
@@ -43,7 +44,8 @@ int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *d
 int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
                                float *P, float *v, const int *active, int C, int ncs, hipStream_t st);
 int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
-                       const float *carry_in, float *out, uint32_t *norm_bits, const int *active, int C, int ncs,
+                       const float *carry_in, const float *zin, float *out, uint32_t *norm_bits, const int *active,
+                       int C, int ncs,
                        hipStream_t st);
 
 // shallow PLRNN
@@ -52,7 +54,8 @@ size_t sh_jacform_lds(int M, int L);
 size_t sh_grads_part_floats(int M, int L, int *nblocks);
 int launch_resjac_shplrnn(const ShArgs &a, const float *z, float *F, float *r, uint32_t *masks, const int *active,
                           hipStream_t st);
-int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, const int *active, hipStream_t st);
+int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, const int *active, const float *gamma,
+                           hipStream_t st);
 int launch_grads_shplrnn(const ShArgs &a, const float *z, const float *lam, const uint32_t *masks, float *part,
                          const deer_grads *gr, hipStream_t st);
 int launch_mse_seed(const float *z, const float *x, float scale, int B, int T, int M, int N, float *g, hipStream_t st);

@@ -92,6 +92,28 @@ def test_solve_reaches_rollout(M, N, B, T, alpha, chunk):
     assert np.array_equal(got[far], (zt > 0)[far])
 
 
+@pytest.mark.parametrize("M,N,B,T,alpha,chunk,bound", [(16, 3, 4, 300, 0.2, 0, 0.05), (16, 3, 3, 300, 0.2, 16, 0.3),
+                                                       (32, 8, 3, 300, 0.1, 16, 0.1), (64, 64, 2, 200, 0.05, 0, 0.1),
+                                                       (5, 2, 5, 120, 0.3, 7, 0.02)])
+def test_safeguard_rejections_reach_rollout(M, N, B, T, alpha, chunk, bound):
+    """A small step bound makes the solver reject updates and retry them damped (the scan
+    uses gamma J~ with gamma < 1, down to the fixed-point step); the iterates alternate
+    between two buffers with per-sequence copy-back.  The result is still the rollout, and
+    more passes than plain Newton's show that the safeguard ran."""
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    c = _case(M, N, B, T, alpha, 600 + M + T)
+    m = oracle_model(c)
+    say("deer_solve safeguard", M, N, B, T, alpha, chunk, bound)
+    plain = D.deer_solve(m, c.x, alpha, N, tol=1e-5, max_iter=100)
+    res = D.deer_solve(m, c.x, alpha, N, tol=1e-5, max_iter=5000, step_bound=bound)
+    assert res["status"] == 0, res
+    ref = O.rollout(m, c.x, alpha, N)
+    assert rel_inf(res["z"].cpu().numpy(), ref) < TOL
+    assert sum(res["iters"]) > sum(plain["iters"])
+    assert all(n < 1e-5 for n in res["norms"])
+
+
 def test_iteration_counts_match_oracle():
     c = _case(16, 3, 4, 800, 0.2, 7)
     m = oracle_model(c)

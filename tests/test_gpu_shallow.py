@@ -109,6 +109,22 @@ def test_shallow_solve_and_adjoint(M, L, N, B, T, alpha, chunk):
         assert rel_inf(out["grads"][k].cpu().numpy(), gr[k]) < TOL, k
 
 
+@pytest.mark.parametrize("M,L,N,B,T,chunk,bound", [(16, 64, 16, 3, 300, 0, 0.05), (20, 40, 5, 3, 200, 32, 0.2)])
+def test_shallow_safeguard_rejections_reach_rollout(M, L, N, B, T, chunk, bound):
+    """Rejected updates retried with the damped stored Jacobians gamma J~ still reach the
+    rollout."""
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    c = _case(M, L, N, B, T, 0.1, 700 + M)
+    m = oracle_model(c)
+    say("deer_solve shallow safeguard", M, L, N, B, T, chunk, bound)
+    plain = D.deer_solve(m, c.x, 0.1, N, tol=1e-5, max_iter=100)
+    res = D.deer_solve(m, c.x, 0.1, N, tol=1e-5, max_iter=5000, step_bound=bound)
+    assert res["status"] == 0, res
+    assert rel_inf(res["z"].cpu().numpy(), O.rollout(m, c.x, 0.1, N)) < TOL
+    assert sum(res["iters"]) > sum(plain["iters"])
+
+
 def test_config3_reduced():
     """Workload 3 (shallow PLRNN M=32, L=256, Lorenz-96) with T reduced to 4096."""
     c = W.make_config(3, B=2, T=4096)

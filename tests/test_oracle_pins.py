@@ -202,6 +202,42 @@ def test_newton_prefix_exactness(init):
     assert full["iters"].max() <= T + 1
 
 
+@pytest.mark.parametrize("gamma", [0.0, 0.5])
+def test_damped_newton_prefix_and_fixed_point(gamma):
+    """The damped step Delta_t = gamma J~_t Delta_{t-1} - r_t (the safeguard of the GPU
+    solve) keeps the fixed point of the GTF residual and the prefix property of the DEER
+    update: after k updates z_1..z_k are exact, for every gamma in [0, 1]."""
+    m = _vanilla(3, 11, w_std=0.8)
+    T = 12
+    x = _x(2, T, 3, 12)
+    alpha = 0.2
+    ref = O.rollout(m, x, alpha, 3)
+    res = O.newton(m, x, alpha, 3, fixed_iters=T, history=True, gamma=gamma)
+    for k, zk in enumerate(res["history"]):
+        if k:
+            assert np.abs(zk[:, :k] - ref[:, :k]).max() < 1e-12, k
+    assert np.abs(res["z"] - ref).max() < 1e-12
+    full = O.newton(m, x, alpha, 3, tol=1e-12, max_iter=100, gamma=gamma)
+    assert full["status"] == "ok" and full["iters"].max() <= T + 1
+
+
+def test_undamped_fixed_point_step_is_local():
+    """gamma = 0 is the fixed-point step z_t <- F(z~_{t-1}): a change of the iterate at
+    step s changes the next iterate at step s + 1 only (z + (F - z) rounds, hence the
+    threshold at step s itself)."""
+    m = _vanilla(4, 21)
+    x = _x(1, 20, 2, 22)
+    z = np.random.default_rng(23).standard_normal((1, 20, 4))
+    base = O.newton(m, x, 0.3, 2, init="user", z_init=z, fixed_iters=1, gamma=0.0)["z"]
+    for s in (0, 7, 19):
+        z2 = z.copy()
+        z2[0, s] += 0.5
+        moved = O.newton(m, x, 0.3, 2, init="user", z_init=z2, fixed_iters=1, gamma=0.0)["z"]
+        diff = np.abs(moved - base).max(axis=2)[0]
+        changed = np.nonzero(diff > 1e-12)[0].tolist()
+        assert changed == ([s + 1] if s + 1 < 20 else []), (s, changed)
+
+
 def test_newton_lands_on_fixed_point_once_masks_match():
     """F is affine on each activation cell, so a Newton update linearised at an iterate
     that shares the fixed point's masks is exact: one update from a small perturbation

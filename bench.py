@@ -37,7 +37,9 @@ def log(*a):
 
 def _plrnn_step(D, model, xd, c, ws_s, ws_a):
     res = D.deer_solve(model, xd, c.alpha, c.n_obs, tol=c.tol, max_iter=c.max_iter, fixed_iters=c.fixed_iters,
-                       ws=ws_s)
+                       ws=ws_s, check=False)
+    if res["status"] != 0:
+        raise RuntimeError(f"deer_solve returned status {res['status']}: {D.load().deer_last_error()}")
     D.deer_adjoint(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a)
     return sum(res["iters"])
 

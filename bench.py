@@ -61,13 +61,14 @@ def kernel_work(c, steps, updates):
     if c.kind == "diag_ssm":
         K = c.n_obs
         elems = steps * B * T * M
+        xin = steps * B * T * 4 * K
         return {
-            # single pass; solve launch: b formed from x on the fly (x read, y written);
-            # adjoint launch: cotangent read, adjoint written
-            "k_diag_scan_lb": ("hbm", elems * 8 + steps * B * T * 4 * K + elems * 16),
-            "k_diag_chunk_fixup": ("hbm", elems * 8 + steps * B * T * 4 * K + elems * 16),
-            "k_diag_chunk_reduce": ("hbm", steps * B * T * 4 * K + elems * 8),
-            "k_diag_grads_partial": ("hbm", elems * 16 + steps * B * T * 4 * K),
+            # forward: b formed from x on the fly; the write pass stores y (8 B per element)
+            "k_diag_seg_write": ("hbm", elems * 8 + xin),
+            # adjoint: cotangent and forward states read, adjoint written (24 B per element),
+            # dlam / dBc accumulated on the way
+            "k_diag_scan_lb_grads": ("hbm", elems * 24 + xin),
+            "k_diag_scan_lb": ("hbm", elems * 16 + xin),
         }
     out = {}
     if c.kind == "plrnn":

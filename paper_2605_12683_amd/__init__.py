@@ -141,7 +141,7 @@ def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, w
     z = _dev(z)
     g = _dev(g)
     shape = (B, T, m.M, 2) if m.kind == "diag_ssm" else (B, T, m.M)
-    lam = torch.empty(shape, device="cuda") if (want_lam or m.kind == "diag_ssm") else None
+    lam = torch.empty(shape, device="cuda") if want_lam else None
     grads = {}
     gs = _b.deer_grads()
     if want_grads:

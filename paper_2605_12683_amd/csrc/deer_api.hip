@@ -183,6 +183,7 @@ struct PlrnnWs {
     float *P, *v, *carry;
     NewtonCtl ctl;
     float *gpart;
+    double *gpart2;
     int C, ncs, MP;
 };
 
@@ -203,6 +204,7 @@ static PlrnnWs carve_plrnn(void *ws, int B, int T, int M, int op, size_t *bytes)
         w.r = c.take<float>((size_t)B * T * M);
     } else {
         w.gpart = c.take<float>(nch * w.MP * (w.MP + 2));
+        w.gpart2 = c.take<double>(reduce_gpart_ws_bytes(w.MP) / sizeof(double));
     }
     *bytes = c.off;
     return w;
@@ -298,13 +300,8 @@ static int check_ws(void *ws, size_t have, size_t need) {
     return DEER_OK;
 }
 
-static size_t diag_bytes(int B, int T, int M, int op) {
-    size_t a = diag_scan_ws_bytes(B, T, M);
-    if (op == DEER_OP_ADJOINT) {
-        size_t g = diag_grads_ws_bytes(B, T, M);
-        if (g > a) a = g;
-    }
-    return a;
+static size_t diag_bytes(int B, int T, int M, int K, int op) {
+    return op == DEER_OP_ADJOINT ? diag_adjoint_ws_bytes(B, T, M, K) : diag_scan_ws_bytes(B, T, M);
 }
 
 // Host-side Newton loop shared by the PLRNN kinds.  `update(active, gamma, zin, zout)` queues
@@ -571,7 +568,7 @@ size_t deer_workspace_bytes(const deer_model *m, int B, int T, int op) {
     deer_forcing f{0.f, 0};
     if (check_common(m, &f, B, T) != DEER_OK) return 0;
     if (op != DEER_OP_SOLVE && op != DEER_OP_ADJOINT) return 0;
-    if (m->kind == DEER_DIAG_SSM) return diag_bytes(B, T, m->M, op);
+    if (m->kind == DEER_DIAG_SSM) return diag_bytes(B, T, m->M, m->L, op);
     if (m->kind == DEER_PLRNN) {
         size_t bytes = 0;
         carve_plrnn(nullptr, B, T, m->M, op, &bytes);
@@ -636,7 +633,7 @@ int deer_solve(const deer_model *m, const deer_forcing *f, const deer_solve_opts
     if (m->kind == DEER_SHPLRNN)
         return solve_shplrnn(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
     if (m->kind == DEER_DIAG_SSM) {
-        if ((rc = check_ws(ws, ws_bytes, diag_bytes(B, T, m->M, DEER_OP_SOLVE)))) return rc;
+        if ((rc = check_ws(ws, ws_bytes, diag_bytes(B, T, m->M, m->L, DEER_OP_SOLVE)))) return rc;
         rc = launch_diag_scan(false, B, T, m->M, m->A, nullptr, m->W, m->L, x, z, ws, st);
         if (rc) return rc;
         if (iters) for (int b = 0; b < B; ++b) iters[b] = 1;
@@ -668,7 +665,7 @@ int deer_adjoint(const deer_model *m, const deer_forcing *f, int B, int T, const
         if ((rc = launch_carry(w.MP, true, w.P, w.v, w.carry, nullptr, nullptr, B, w.ncs, st))) return rc;
         if ((rc = launch_fixup_rev_plrnn(a, w.masks, g, scale, z, w.carry, lam, w.gpart, w.C, w.ncs, st))) return rc;
         if (grads && (grads->A || grads->W || grads->h)) {
-            if ((rc = launch_reduce_gpart(w.gpart, B * w.ncs, w.MP, m->M, grads->A, grads->W, grads->h, st))) return rc;
+            if ((rc = launch_reduce_gpart(w.gpart, B * w.ncs, w.MP, m->M, grads->A, grads->W, grads->h, w.gpart2, st))) return rc;
         }
         return DEER_OK;
     }
@@ -699,14 +696,10 @@ int deer_adjoint(const deer_model *m, const deer_forcing *f, int B, int T, const
     }
     if (m->kind == DEER_DIAG_SSM) {
         if (!g) { set_error("DIAG_SSM adjoint needs the cotangent g"); return DEER_ERR_INVALID_ARG; }
-        if ((rc = check_ws(ws, ws_bytes, diag_bytes(B, T, m->M, DEER_OP_ADJOINT)))) return rc;
-        float *out = lam;
-        if (!out) { set_error("DIAG_SSM adjoint needs the lam output buffer"); return DEER_ERR_INVALID_ARG; }
-        if ((rc = launch_diag_scan(true, B, T, m->M, m->A, g, nullptr, m->L, nullptr, out, ws, st))) return rc;
-        if (grads && (grads->A || grads->W)) {
-            if ((rc = launch_diag_grads(B, T, m->M, m->L, out, z, x, grads->A, grads->W, ws, st))) return rc;
-        }
-        return DEER_OK;
+        if ((rc = check_ws(ws, ws_bytes, diag_bytes(B, T, m->M, m->L, DEER_OP_ADJOINT)))) return rc;
+        float *dlam = grads ? grads->A : nullptr, *dBc = grads ? grads->W : nullptr;
+        if (!lam && !dlam && !dBc) return DEER_OK;
+        return launch_diag_adjoint(B, T, m->M, m->L, m->A, g, z, x, lam, dlam, dBc, ws, st);
     }
     set_error("deer_adjoint: model kind %d not supported yet", m->kind);
     return DEER_ERR_INVALID_ARG;

@@ -158,17 +158,26 @@ __device__ __forceinline__ void pub_word(unsigned long long *p, float v) {
     const unsigned long long w = (1ull << 32) | (unsigned long long)(uint32_t)__float_as_uint(v);
     __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-template <bool PROJ>
+// GRADS (reverse scans only): the adjoint a_tau = y is combined on the fly with the forward
+// states h and the inputs x into per-block partial sums of
+//   dlam_m = sum a_tau conj(h_{tau-1}),  dBc_{m,k} = sum a_tau x_tau[k]
+// (layout part[(k * B * ntile * nq + chain * nq + q) * DTC + ch], k < 2 + 2K); yout may then
+// be null (the adjoint itself not stored).
+constexpr int DNV = 10;   // 2 + 2 K partial values per channel, K <= 4
+
+template <bool PROJ, bool GRADS>
 __global__ __launch_bounds__(DNW * 64) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_diag_scan_lb(const float *__restrict__ lam, int conj_lam,
                                                           const float *__restrict__ bin, const float *__restrict__ Bc,
                                                           int K, const float *__restrict__ u, int rev, int B, int T,
                                                           int M, int ntile, int nq, unsigned int *__restrict__ ticket,
                                                           unsigned long long *__restrict__ aggw,
                                                           unsigned long long *__restrict__ incw,
-                                                          float *__restrict__ yout) {
+                                                          float *__restrict__ yout, const float *__restrict__ hfwd,
+                                                          float *__restrict__ part) {
     __shared__ float2 sub[DNW * 4][DTC];
     __shared__ float2 xq[DTC];
-    __shared__ float xs[PROJ ? DCH * 4 : 1];
+    __shared__ float xs[(PROJ || GRADS) ? DCH * 4 : 1];
+    __shared__ float red[GRADS ? DNW : 1][DTC][DNV];
     __shared__ unsigned int vid_s;
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, j = lane >> 4, ch = lane & 15;
     const int usub = w * 4 + j;
@@ -194,12 +203,14 @@ __global__ __launch_bounds__(DNW * 64) __attribute__((amdgpu_waves_per_eu(4, 8))
         }
     }
     const long p0 = (long)q * DCH + (long)usub * DS;
-    if (PROJ) {
-        // inputs of this chunk staged in LDS with coalesced loads (forward only: tau = p)
+    if (PROJ || GRADS) {
+        // inputs of this chunk staged in LDS with coalesced loads, in position order
+        // (PROJ: forward, tau = p; GRADS: reverse, tau = T - 1 - p)
         const long n = (long)DCH * K;
         for (long e = tid; e < n; e += DNW * 64) {
             const long p = (long)q * DCH + e / K;
-            xs[e] = p < T ? u[((long)b * (T + 1) + p) * K + (e % K)] : 0.f;
+            const long tau = GRADS ? (T - 1 - p) : p;
+            xs[e] = p < T ? u[((long)b * (T + 1) + tau) * K + (e % K)] : 0.f;
         }
         __syncthreads();
     }
@@ -316,6 +327,9 @@ __global__ __launch_bounds__(DNW * 64) __attribute__((amdgpu_waves_per_eu(4, 8))
         yr = (float)((double)pr + (Lu.re * X.x - Lu.im * X.y));
         yi = (float)((double)pi + (Lu.re * X.y + Lu.im * X.x));
     }
+    float acc[DNV];
+#pragma unroll
+    for (int k = 0; k < DNV; ++k) acc[k] = 0.f;
 #pragma unroll
     for (int s = 0; s < DS; ++s) {
         const float nr = fmaf(lr, yr, fmaf(-li, yi, bv[s].x));
@@ -325,8 +339,46 @@ __global__ __launch_bounds__(DNW * 64) __attribute__((amdgpu_waves_per_eu(4, 8))
         const long p = p0 + s;
         if (mok && p < T) {
             const long tau = rev ? (T - 1 - p) : p;
-            const v2f o2 = {yr, yi};
-            __builtin_nontemporal_store(o2, reinterpret_cast<v2f *>(yout + (((long)b * T + tau) * M + m) * 2));
+            if (yout) {
+                const v2f o2 = {yr, yi};
+                __builtin_nontemporal_store(o2, reinterpret_cast<v2f *>(yout + (((long)b * T + tau) * M + m) * 2));
+            }
+            if (GRADS) {
+                if (tau > 0) {
+                    const v2f hv = __builtin_nontemporal_load(
+                        reinterpret_cast<const v2f *>(hfwd + (((long)b * T + tau - 1) * M + m) * 2));
+                    acc[0] = fmaf(yr, hv.x, fmaf(yi, hv.y, acc[0]));
+                    acc[1] = fmaf(yi, hv.x, fmaf(-yr, hv.y, acc[1]));
+                }
+                const float *xu = xs + (long)(usub * DS + s) * K;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (k < K) {
+                        acc[2 + 2 * k] = fmaf(yr, xu[k], acc[2 + 2 * k]);
+                        acc[3 + 2 * k] = fmaf(yi, xu[k], acc[3 + 2 * k]);
+                    }
+            }
+        }
+    }
+    if (GRADS) {
+        // sum over the 4 sub-chunks of a wave (lanes ch, ch + 16, ch + 32, ch + 48), then over waves
+#pragma unroll
+        for (int k = 0; k < DNV; ++k) {
+            acc[k] += __shfl_xor(acc[k], 16, 64);
+            acc[k] += __shfl_xor(acc[k], 32, 64);
+        }
+        if (j == 0) {
+#pragma unroll
+            for (int k = 0; k < DNV; ++k) red[w][ch][k] = acc[k];
+        }
+        __syncthreads();
+        const int nv = 2 + 2 * K;
+        if (tid < DTC * nv) {
+            const int c2 = tid % DTC, k = tid / DTC;
+            float sum = 0.f;
+#pragma unroll
+            for (int w2 = 0; w2 < DNW; ++w2) sum += red[w2][c2][k];
+            part[(((long)k * B * ntile + st) * nq + q) * DTC + c2] = sum;
         }
     }
 }
@@ -395,6 +447,203 @@ __global__ __launch_bounds__(256) void k_diag_carry(const float *__restrict__ la
     }
 }
 
+// ---------------------------------------------------------------------------------------
+// Forward scan with the input projection fused (y_t = lam y_{t-1} + Bc x_t, y_{-1} = 0, in
+// 0-based array positions): the only HBM stream is the output, so the scan is write-bound.
+// A wave owns 64 channels (lane = channel: one 512-byte row per step at M = 64) and a
+// segment of SEG = 64 * SEG_L consecutive steps that it walks sequentially.  The inputs of
+// the segment are loaded once, lane l holding steps SEG_L l .. SEG_L l + SEG_L - 1, and are
+// broadcast to the wave with v_readlane as the walk reaches them.  No LDS, no barriers, no
+// look-back.
+//   k_diag_seg<false>  segment aggregates from zero (reads the inputs only)
+//   k_diag_seg_carry   carries across segments in float64 (three-level: groups of segments)
+//   k_diag_seg<true>   re-walk of every segment from its carry, y written (non-temporal)
+// ---------------------------------------------------------------------------------------
+constexpr int SEG_L = 8;
+constexpr int SEG = 64 * SEG_L;
+
+__device__ __forceinline__ float lane_bcast(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+template <bool WRITE, int K>
+__global__ __launch_bounds__(256) void k_diag_seg(const float *__restrict__ lam, const float *__restrict__ Bc,
+                                                  const float *__restrict__ u, int B, int T, int M, int nseg,
+                                                  int ntile, float2 *__restrict__ agg,
+                                                  const float2 *__restrict__ carry, float *__restrict__ y) {
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const long wid = (long)blockIdx.x * 4 + wv;          // (sequence, segment, channel tile)
+    if (wid >= (long)B * nseg * ntile) return;
+    const int tile = (int)(wid % ntile);
+    const long bs = wid / ntile;                          // sequence * nseg + segment
+    const int seg = (int)(bs % nseg), b = (int)(bs / nseg);
+    const int m = tile * 64 + lane;
+    const bool mok = m < M;
+    const int t0 = seg * SEG, t1 = min(t0 + SEG, T);
+    // inputs of the segment: lane l holds rows t0 + SEG_L l + s, s < SEG_L
+    float xv[SEG_L * K];
+    {
+        const float *xr = u + ((long)b * (T + 1) + t0 + SEG_L * lane) * K;
+        const int nrow = min(SEG_L, t1 - t0 - SEG_L * lane);
+#pragma unroll
+        for (int e = 0; e < SEG_L * K; ++e) xv[e] = e < nrow * K ? xr[e] : 0.f;
+    }
+    float lr = 0.f, li = 0.f, br[K], bi[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) br[k] = bi[k] = 0.f;
+    if (mok) {
+        lr = lam[2 * m];
+        li = lam[2 * m + 1];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            br[k] = Bc[(m * K + k) * 2];
+            bi[k] = Bc[(m * K + k) * 2 + 1];
+        }
+    }
+    float hr = 0.f, hi = 0.f;
+    if (WRITE && mok) {
+        const float2 X = carry[bs * M + m];
+        hr = X.x;
+        hi = X.y;
+    }
+    float *yb = y + ((long)b * T + t0) * M * 2 + 2 * m;
+    const int ngrp = (t1 - t0 + SEG_L - 1) / SEG_L;
+    for (int gq = 0; gq < ngrp; ++gq) {
+        const int tb = t0 + gq * SEG_L;
+#pragma unroll
+        for (int s = 0; s < SEG_L; ++s) {
+            float vr = 0.f, vi = 0.f;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const float xk = lane_bcast(xv[s * K + k], gq);
+                vr = fmaf(br[k], xk, vr);
+                vi = fmaf(bi[k], xk, vi);
+            }
+            if (tb + s < t1) {
+                const float nr = fmaf(lr, hr, fmaf(-li, hi, vr));
+                const float ni = fmaf(lr, hi, fmaf(li, hr, vi));
+                hr = nr;
+                hi = ni;
+                if (WRITE && mok) {
+                    const v2f o2 = {hr, hi};
+                    __builtin_nontemporal_store(o2, reinterpret_cast<v2f *>(yb + (long)(tb - t0 + s) * M * 2));
+                }
+            }
+        }
+    }
+    if (!WRITE && mok) agg[bs * M + m] = make_float2(hr, hi);
+}
+
+// carry[s] = state at the end of segment s - 1:  X_0 = 0,  X_{s+1} = Lambda X_s + A_s,
+// Lambda = lam^SEG (every segment but the last is full; the last aggregate is not needed).
+// Block = (sequence, 64-channel tile), threads = (group g of CG consecutive segments, channel):
+// group aggregates, a sequential pass over the 16 groups, then every group re-walked from its
+// carry.  Serial depth 2 CG + 16 instead of nseg.
+constexpr int SEG_NG = 16;
+
+__global__ __launch_bounds__(1024) void k_diag_seg_carry(const float *__restrict__ lam, int B, int M, int nseg,
+                                                         int ntile, const float2 *__restrict__ agg,
+                                                         float2 *__restrict__ carry) {
+    __shared__ double ga[SEG_NG][64][2];
+    const int b = blockIdx.x / ntile, tile = blockIdx.x % ntile;
+    const int ch = threadIdx.x & 63, grp = threadIdx.x >> 6;
+    const int m = tile * 64 + ch;
+    const bool mok = m < M;
+    const int CG = (nseg + SEG_NG - 1) / SEG_NG;
+    const int s0 = grp * CG, s1 = min(s0 + CG, nseg);
+    cd L = {0.0, 0.0};
+    if (mok) L = cpow(cd{(double)lam[2 * m], (double)lam[2 * m + 1]}, SEG);
+    const long base = (long)b * nseg;
+    double ar = 0.0, ai = 0.0;
+    if (mok) {
+        for (int s = s0; s < s1; ++s) {
+            const float2 a = agg[(base + s) * M + m];
+            const double nr = L.re * ar - L.im * ai + (double)a.x;
+            const double ni = L.re * ai + L.im * ar + (double)a.y;
+            ar = nr;
+            ai = ni;
+        }
+    }
+    ga[grp][ch][0] = ar;
+    ga[grp][ch][1] = ai;
+    __syncthreads();
+    if (grp == 0 && mok) {
+        const cd LG = cpow(L, CG);
+        double cr = 0.0, ci = 0.0;
+        for (int g2 = 0; g2 < SEG_NG; ++g2) {
+            const double xr = ga[g2][ch][0], xi = ga[g2][ch][1];
+            ga[g2][ch][0] = cr;
+            ga[g2][ch][1] = ci;
+            const double nr = LG.re * cr - LG.im * ci + xr;
+            const double ni = LG.re * ci + LG.im * cr + xi;
+            cr = nr;
+            ci = ni;
+        }
+    }
+    __syncthreads();
+    if (!mok) return;
+    double xr = ga[grp][ch][0], xi = ga[grp][ch][1];
+    for (int s = s0; s < s1; ++s) {
+        const float2 a = agg[(base + s) * M + m];
+        carry[(base + s) * M + m] = make_float2((float)xr, (float)xi);
+        const double nr = L.re * xr - L.im * xi + (double)a.x;
+        const double ni = L.re * xi + L.im * xr + (double)a.y;
+        xr = nr;
+        xi = ni;
+    }
+}
+
+static bool diag_seg_enabled() {
+    const char *e = getenv("DEER_DIAG_SEG");
+    return !e || atoi(e) != 0;
+}
+
+static size_t diag_seg_ws_bytes(int B, int T, int M) {
+    const size_t nseg = (T + SEG - 1) / SEG;
+    const size_t one = ((size_t)B * nseg * M * sizeof(float2) + 255) & ~(size_t)255;
+    return 2 * one;
+}
+
+static int launch_diag_seg(int B, int T, int M, const float *lam, const float *Bc, int K, const float *u, float *y,
+                           void *ws, hipStream_t st) {
+    const int nseg = (T + SEG - 1) / SEG;
+    const int ntile = (M + 63) / 64;
+    const size_t one = ((size_t)B * nseg * M * sizeof(float2) + 255) & ~(size_t)255;
+    float2 *agg = (float2 *)ws;
+    float2 *carry = (float2 *)((char *)ws + one);
+    const long waves = (long)B * nseg * ntile;
+    const int grid = (int)((waves + 3) / 4);
+#define SEGK(WR, KV, A, C, Y) \
+    hipLaunchKernelGGL((k_diag_seg<WR, KV>), dim3(grid), dim3(256), 0, st, lam, Bc, u, B, T, M, nseg, ntile, A, C, Y)
+#define SEGALL(WR, A, C, Y)                  \
+    switch (K) {                             \
+        case 1: SEGK(WR, 1, A, C, Y); break; \
+        case 2: SEGK(WR, 2, A, C, Y); break; \
+        case 3: SEGK(WR, 3, A, C, Y); break; \
+        default: SEGK(WR, 4, A, C, Y); break; \
+    }
+    {
+        KTimer _kt("k_diag_seg_reduce", st);
+        SEGALL(false, agg, (const float2 *)nullptr, (float *)nullptr)
+    }
+    DEER_LAUNCH_CHECK("k_diag_seg<reduce>");
+    {
+        KTimer _kt("k_diag_seg_carry", st);
+        hipLaunchKernelGGL(k_diag_seg_carry, dim3(B * ntile), dim3(64 * SEG_NG), 0, st, lam, B, M, nseg, ntile,
+                           (const float2 *)agg, carry);
+    }
+    DEER_LAUNCH_CHECK("k_diag_seg_carry");
+    {
+        KTimer _kt("k_diag_seg_write", st);
+        SEGALL(true, (float2 *)nullptr, (const float2 *)carry, y)
+    }
+#undef SEGALL
+#undef SEGK
+    DEER_LAUNCH_CHECK("k_diag_seg<write>");
+    return DEER_OK;
+}
+
 static bool diag_three_pass() {
     const char *e = getenv("DEER_DIAG_3PASS");
     return e && atoi(e) != 0;
@@ -407,7 +656,9 @@ size_t diag_scan_ws_bytes(int B, int T, int M) {
     const size_t three = 2 * ((one + 255) & ~(size_t)255);
     const size_t words = (size_t)B * ntile * nq * DTC * 2 * sizeof(unsigned long long);
     const size_t single = 256 + 2 * ((words + 255) & ~(size_t)255);
-    return three > single ? three : single;
+    size_t need = three > single ? three : single;
+    const size_t seg = diag_seg_ws_bytes(B, T, M);
+    return need > seg ? need : seg;
 }
 
 int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const float *b, const float *Bc, int K,
@@ -416,6 +667,7 @@ int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const floa
     const int nq = (T + DCH - 1) / DCH;
     const int nblk = B * ntile * nq;
     const int conj_lam = rev ? 1 : 0;
+    if (!b && !rev && diag_seg_enabled()) return launch_diag_seg(B, T, M, lam, Bc, K, u, y, ws, st);
     if (!diag_three_pass()) {
         const size_t nwords = (size_t)B * ntile * nq * DTC * 2;
         const size_t wbytes = (nwords * sizeof(unsigned long long) + 255) & ~(size_t)255;
@@ -432,11 +684,13 @@ int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const floa
         {
             KTimer _kt("k_diag_scan_lb", st);
             if (b)
-                hipLaunchKernelGGL(k_diag_scan_lb<false>, dim3(nblk), dim3(DNW * 64), 0, st, lam, conj_lam, b, Bc, K,
-                                   u, rev ? 1 : 0, B, T, M, ntile, nq, ticket, aggw, incw, y);
+                hipLaunchKernelGGL((k_diag_scan_lb<false, false>), dim3(nblk), dim3(DNW * 64), 0, st, lam, conj_lam, b,
+                                   Bc, K, u, rev ? 1 : 0, B, T, M, ntile, nq, ticket, aggw, incw, y,
+                                   (const float *)nullptr, (float *)nullptr);
             else
-                hipLaunchKernelGGL(k_diag_scan_lb<true>, dim3(nblk), dim3(DNW * 64), 0, st, lam, conj_lam, b, Bc, K,
-                                   u, rev ? 1 : 0, B, T, M, ntile, nq, ticket, aggw, incw, y);
+                hipLaunchKernelGGL((k_diag_scan_lb<true, false>), dim3(nblk), dim3(DNW * 64), 0, st, lam, conj_lam, b,
+                                   Bc, K, u, rev ? 1 : 0, B, T, M, ntile, nq, ticket, aggw, incw, y,
+                                   (const float *)nullptr, (float *)nullptr);
         }
         DEER_LAUNCH_CHECK("k_diag_scan_lb");
         return DEER_OK;
@@ -464,105 +718,103 @@ int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const floa
     return DEER_OK;
 }
 
-}  // namespace deer
+// float64 sums of the fused-scan partials.  Stage 1: block = (channel tile, value k, slice of
+// the B * nq chunk rows), lanes (row r, channel ch); stage 2 sums the slices.
+constexpr int DGS = 64;   // slices
 
-namespace deer {
-
-// Gradients of the diagonal SSM parameters from the adjoint a and the forward states h:
-//   dlam_m = sum_{b,t} a_t conj(h_{t-1}),  dBc_{m,k} = sum_{b,t} a_t u_t[k]  (u_t = x_{t-1})
-// Pass 1: block = 16 channels x 16 time lanes over a slice of DGT positions -> fp32 partials.
-// Pass 2: float64 sum of the partials.
-namespace {
-constexpr int DGT = 4096;
-}
-
-__global__ __launch_bounds__(256) void k_diag_grads_partial(const float *__restrict__ a, const float *__restrict__ h,
-                                                            const float *__restrict__ x, int K, int B, int T, int M,
-                                                            int ntile, int nsl, float *__restrict__ part) {
-    __shared__ float red[16][16][2 + 8];
-    const int tl = threadIdx.x >> 4, ch = threadIdx.x & 15;
-    const int sl = blockIdx.x % nsl, st = blockIdx.x / nsl;
-    const int b = st / ntile, m = (st % ntile) * DTC + ch;
-    const bool mok = m < M;
-    float acc[2 + 8];
-#pragma unroll
-    for (int k = 0; k < 10; ++k) acc[k] = 0.f;
-    const int t0 = sl * DGT, t1 = min(t0 + DGT, T);
-    if (mok) {
-        for (int t = t0 + tl; t < t1; t += 16) {
-            const float2 av = *reinterpret_cast<const float2 *>(a + (((long)b * T + t) * M + m) * 2);
-            if (t > 0) {
-                const float2 hv = *reinterpret_cast<const float2 *>(h + (((long)b * T + t - 1) * M + m) * 2);
-                acc[0] = fmaf(av.x, hv.x, fmaf(av.y, hv.y, acc[0]));
-                acc[1] = fmaf(av.y, hv.x, fmaf(-av.x, hv.y, acc[1]));
-            }
-            const float *xu = x + ((long)b * (T + 1) + t) * K;
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                if (k < K) {
-                    const float uk = xu[k];
-                    acc[2 + 2 * k] = fmaf(av.x, uk, acc[2 + 2 * k]);
-                    acc[3 + 2 * k] = fmaf(av.y, uk, acc[3 + 2 * k]);
-                }
-        }
-    }
-#pragma unroll
-    for (int k = 0; k < 10; ++k) red[tl][ch][k] = acc[k];
-    __syncthreads();
-    if (tl == 0 && mok) {
-        const int nv = 2 + 2 * K;
-        for (int k = 0; k < nv; ++k) {
-            float s = 0.f;
-            for (int r = 0; r < 16; ++r) s += red[r][ch][k];
-            part[(((long)st * nsl + sl) * DTC + ch) * 10 + k] = s;
-        }
-    }
-}
-
-__global__ void k_diag_grads_final(const float *__restrict__ part, int K, int B, int M, int ntile, int nsl,
-                                   float *__restrict__ dlam, float *__restrict__ dBc) {
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;   // (m, k)
-    const int nv = 2 + 2 * K;
-    if (e >= M * nv) return;
-    const int m = e / nv, k = e % nv;
-    const int tile = m / DTC, ch = m % DTC;
+__global__ __launch_bounds__(256) void k_diag_grads_sum1(const float *__restrict__ part, int B, int ntile, int nq,
+                                                         double *__restrict__ part2) {
+    __shared__ double red[16][DTC];
+    const int sl = blockIdx.x % DGS, tk = blockIdx.x / DGS;   // tk = k * ntile + tile
+    const int tile = tk % ntile, k = tk / ntile;
+    const int tid = threadIdx.x, r = tid / DTC, ch = tid % DTC;
+    const long rows = (long)B * nq;
+    const long r0 = rows * sl / DGS, r1 = rows * (sl + 1) / DGS;
     double s = 0.0;
-    for (int b = 0; b < B; ++b) {
-        const int st = b * ntile + tile;
-        for (int sl = 0; sl < nsl; ++sl) s += (double)part[(((long)st * nsl + sl) * DTC + ch) * 10 + k];
+    for (long row = r0 + r; row < r1; row += 16) {
+        const long bb = row / nq, q = row % nq;
+        s += (double)part[(((long)k * B * ntile + bb * ntile + tile) * nq + q) * DTC + ch];
     }
+    red[r][ch] = s;
+    __syncthreads();
+    if (tid < DTC) {
+        double t = 0.0;
+        for (int r2 = 0; r2 < 16; ++r2) t += red[r2][tid];
+        part2[((long)tk * DGS + sl) * DTC + tid] = t;
+    }
+}
+
+__global__ __launch_bounds__(64) void k_diag_grads_sum2(const double *__restrict__ part2, int K, int M, int ntile,
+                                                        float *__restrict__ dlam, float *__restrict__ dBc) {
+    const int e = blockIdx.x * 64 + threadIdx.x;   // (k, m)
+    if (e >= (2 + 2 * K) * ntile * DTC) return;
+    const int ch = e % DTC, tk = e / DTC;
+    const int tile = tk % ntile, k = tk / ntile;
+    const int m = tile * DTC + ch;
+    if (m >= M) return;
+    double t = 0.0;
+    for (int sl = 0; sl < DGS; ++sl) t += part2[((long)tk * DGS + sl) * DTC + ch];
     if (k < 2) {
-        if (dlam) dlam[2 * m + k] = (float)s;
+        if (dlam) dlam[2 * m + k] = (float)t;
     } else if (dBc) {
         const int kk = (k - 2) / 2, ri = (k - 2) % 2;
-        dBc[(m * K + kk) * 2 + ri] = (float)s;
+        dBc[(m * K + kk) * 2 + ri] = (float)t;
     }
 }
 
-size_t diag_grads_ws_bytes(int B, int T, int M) {
+size_t diag_adjoint_ws_bytes(int B, int T, int M, int K) {
     const long ntile = (M + DTC - 1) / DTC;
-    const long nsl = (T + DGT - 1) / DGT;
-    return (((size_t)B * ntile * nsl * DTC * 10 * sizeof(float)) + 255) & ~(size_t)255;
+    const long nq = (T + DCH - 1) / DCH;
+    const size_t words = (size_t)B * ntile * nq * DTC * 2 * sizeof(unsigned long long);
+    const size_t parts = (size_t)(2 + 2 * K) * B * ntile * nq * DTC * sizeof(float);
+    const size_t parts2 = (size_t)(2 + 2 * K) * ntile * DGS * DTC * sizeof(double);
+    return 256 + 2 * ((words + 255) & ~(size_t)255) + ((parts + 255) & ~(size_t)255) + parts2;
 }
 
-int launch_diag_grads(int B, int T, int M, int K, const float *a, const float *h, const float *x, float *dlam,
-                      float *dBc, void *ws, hipStream_t st) {
+// Reverse scan of the cotangent g with the parameter gradients fused (dlam, dBc may be
+// null; lam_out may be null).
+int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const float *g, const float *h, const float *x,
+                        float *lam_out, float *dlam, float *dBc, void *ws, hipStream_t st) {
     const int ntile = (M + DTC - 1) / DTC;
-    const int nsl = (T + DGT - 1) / DGT;
-    float *part = (float *)ws;
+    const int nq = (T + DCH - 1) / DCH;
+    const int nblk = B * ntile * nq;
+    const size_t nwords = (size_t)B * ntile * nq * DTC * 2;
+    const size_t wbytes = (nwords * sizeof(unsigned long long) + 255) & ~(size_t)255;
+    unsigned int *ticket = (unsigned int *)ws;
+    unsigned long long *aggw = (unsigned long long *)((char *)ws + 256);
+    unsigned long long *incw = (unsigned long long *)((char *)ws + 256 + wbytes);
+    float *part = (float *)((char *)ws + 256 + 2 * wbytes);
+    const size_t pbytes = ((size_t)(2 + 2 * K) * B * ntile * nq * DTC * sizeof(float) + 255) & ~(size_t)255;
+    double *part2 = (double *)((char *)part + pbytes);
     {
-        KTimer _kt("k_diag_grads_partial", st);
-        hipLaunchKernelGGL(k_diag_grads_partial, dim3(B * ntile * nsl), dim3(256), 0, st, a, h, x, K, B, T, M, ntile, nsl,
-                           part);
+        KTimer _kt("k_zero_u64", st);
+        const size_t n = 32 + 2 * wbytes / sizeof(unsigned long long);
+        const int grid = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+        hipLaunchKernelGGL(k_zero_u64, dim3(grid), dim3(256), 0, st, (unsigned long long *)ws, n);
     }
-    DEER_LAUNCH_CHECK("k_diag_grads_partial");
-    const int n = M * (2 + 2 * K);
+    DEER_LAUNCH_CHECK("k_zero_u64");
+    const bool grads = dlam || dBc;
     {
-        KTimer _kt("k_diag_grads_final", st);
-        hipLaunchKernelGGL(k_diag_grads_final, dim3((n + 255) / 256), dim3(256), 0, st, part, K, B, M, ntile, nsl, dlam,
-                           dBc);
+        KTimer _kt(grads ? "k_diag_scan_lb_grads" : "k_diag_scan_lb", st);
+        if (grads)
+            hipLaunchKernelGGL((k_diag_scan_lb<false, true>), dim3(nblk), dim3(DNW * 64), 0, st, lam, 1, g,
+                               (const float *)nullptr, K, x, 1, B, T, M, ntile, nq, ticket, aggw, incw, lam_out, h,
+                               part);
+        else
+            hipLaunchKernelGGL((k_diag_scan_lb<false, false>), dim3(nblk), dim3(DNW * 64), 0, st, lam, 1, g,
+                               (const float *)nullptr, K, x, 1, B, T, M, ntile, nq, ticket, aggw, incw, lam_out,
+                               (const float *)nullptr, (float *)nullptr);
     }
-    DEER_LAUNCH_CHECK("k_diag_grads_final");
+    DEER_LAUNCH_CHECK("k_diag_scan_lb");
+    if (grads) {
+        KTimer _kt("k_diag_grads_sum", st);
+        const int nv = 2 + 2 * K;
+        hipLaunchKernelGGL(k_diag_grads_sum1, dim3(ntile * nv * DGS), dim3(256), 0, st, (const float *)part, B, ntile, nq,
+                           part2);
+        hipLaunchKernelGGL(k_diag_grads_sum2, dim3((nv * ntile * DTC + 63) / 64), dim3(64), 0, st,
+                           (const double *)part2, K, M, ntile, dlam, dBc);
+        DEER_LAUNCH_CHECK("k_diag_grads_sum");
+    }
     return DEER_OK;
 }
 

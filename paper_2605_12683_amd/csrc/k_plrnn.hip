@@ -692,23 +692,39 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn(const float *__restrict_
     }
 }
 
-// sum the per-chunk partials in float64: one thread per entry of [MP][MP + 2]
-__global__ void k_reduce_gpart(const float *__restrict__ gpart, int nchains, int MP, int M, float *__restrict__ dA,
-                               float *__restrict__ dW, float *__restrict__ dh) {
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    const int stride = MP * (MP + 2);
-    if (e >= stride) return;
-    const int i = e / (MP + 2), j = e % (MP + 2);
-    if (i >= M) return;
-    if (j < MP && j >= M) return;
-    double s0 = 0.0, s1 = 0.0;
-    int ch = 0;
-    for (; ch + 1 < nchains; ch += 2) {
-        s0 += (double)gpart[(size_t)ch * stride + e];
-        s1 += (double)gpart[(size_t)(ch + 1) * stride + e];
+// sum the per-chunk partials in float64 in two stages: blocks over slices of the chains
+// (consecutive threads read consecutive entries of [MP][MP + 2]), then the slices
+constexpr int GP_SLICES = 64;
+
+__global__ __launch_bounds__(256) void k_reduce_gpart1(const float *__restrict__ gpart, int nchains, int n,
+                                                       double *__restrict__ part2) {
+    const int sl = blockIdx.x;
+    const int c0 = (int)((long)nchains * sl / GP_SLICES), c1 = (int)((long)nchains * (sl + 1) / GP_SLICES);
+    for (int e = threadIdx.x; e < n; e += 256) {
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+        int ch = c0;
+        for (; ch + 3 < c1; ch += 4) {
+            s0 += (double)gpart[(size_t)ch * n + e];
+            s1 += (double)gpart[(size_t)(ch + 1) * n + e];
+            s2 += (double)gpart[(size_t)(ch + 2) * n + e];
+            s3 += (double)gpart[(size_t)(ch + 3) * n + e];
+        }
+        for (; ch < c1; ++ch) s0 += (double)gpart[(size_t)ch * n + e];
+        part2[(size_t)sl * n + e] = (s0 + s1) + (s2 + s3);
     }
-    if (ch < nchains) s0 += (double)gpart[(size_t)ch * stride + e];
-    const float v = (float)(s0 + s1);
+}
+
+__global__ __launch_bounds__(256) void k_reduce_gpart2(const double *__restrict__ part2, int MP, int M,
+                                                       float *__restrict__ dA, float *__restrict__ dW,
+                                                       float *__restrict__ dh) {
+    const int n = MP * (MP + 2);
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e >= n) return;
+    const int i = e / (MP + 2), j = e % (MP + 2);
+    if (i >= M || (j < MP && j >= M)) return;
+    double s = 0.0;
+    for (int sl = 0; sl < GP_SLICES; ++sl) s += part2[(size_t)sl * n + e];
+    const float v = (float)s;
     if (j < MP) {
         if (dW) dW[i * M + j] = v;
     } else if (j == MP) {
@@ -717,6 +733,8 @@ __global__ void k_reduce_gpart(const float *__restrict__ gpart, int nchains, int
         if (dh) dh[i] = v;
     }
 }
+
+size_t reduce_gpart_ws_bytes(int MP) { return (size_t)GP_SLICES * MP * (MP + 2) * sizeof(double); }
 
 // ---------------------------------------------------------------------------------------
 // host launchers
@@ -825,11 +843,13 @@ int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
 }
 
 int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *dA, float *dW, float *dh,
-                        hipStream_t st) {
+                        double *part2, hipStream_t st) {
     const int n = MP * (MP + 2);
     {
         KTimer _kt("k_reduce_gpart", st);
-        hipLaunchKernelGGL(k_reduce_gpart, dim3((n + 255) / 256), dim3(256), 0, st, gpart, nchains, MP, M, dA, dW, dh);
+        hipLaunchKernelGGL(k_reduce_gpart1, dim3(GP_SLICES), dim3(256), 0, st, gpart, nchains, n, part2);
+        hipLaunchKernelGGL(k_reduce_gpart2, dim3((n + 255) / 256), dim3(256), 0, st, (const double *)part2, MP, M, dA,
+                           dW, dh);
     }
     DEER_LAUNCH_CHECK("k_reduce_gpart");
     return DEER_OK;

@@ -38,7 +38,8 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
 int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *g, float seed_scale, const float *z,
                            const float *carry_in, float *lam, float *gpart, int C, int ncs, hipStream_t st);
 int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *dA, float *dW, float *dh,
-                        hipStream_t st);
+                        double *part2, hipStream_t st);
+size_t reduce_gpart_ws_bytes(int MP);
 
 // dense stored-Jacobian scan (mode: 0 Newton fix-up, 1 bare forward scan, 2 reverse)
 int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
@@ -64,9 +65,9 @@ int launch_mse_seed(const float *z, const float *x, float scale, int B, int T, i
 size_t diag_scan_ws_bytes(int B, int T, int M);
 int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const float *b, const float *Bc, int K,
                      const float *u, float *y, void *ws, hipStream_t st);
-size_t diag_grads_ws_bytes(int B, int T, int M);
-int launch_diag_grads(int B, int T, int M, int K, const float *a, const float *h, const float *x, float *dlam,
-                      float *dBc, void *ws, hipStream_t st);
+size_t diag_adjoint_ws_bytes(int B, int T, int M, int K);
+int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const float *g, const float *h, const float *x,
+                        float *lam_out, float *dlam, float *dBc, void *ws, hipStream_t st);
 
 // small utilities
 int launch_fill_teacher(int B, int T, int M, int N, const float *x, float *z, hipStream_t st);

@@ -57,3 +57,35 @@ def test_diag_solve_fused_projection_and_adjoint():
     assert rel_inf(_c(out["lam"].cpu().numpy()), ref["a"]) < TOL
     assert rel_inf(_c(out["grads"]["lam"].cpu().numpy()), ref["grads"]["lam"]) < TOL
     assert rel_inf(_c(out["grads"]["Bc"].cpu().numpy()), ref["grads"]["Bc"]) < TOL
+
+
+@pytest.mark.parametrize("B,T,M,K", [(1, 1, 1, 1), (1, 5, 3, 2), (2, 511, 16, 3), (1, 1025, 17, 4),
+                                     (3, 2049, 64, 3), (2, 5000, 70, 1), (1, 70000, 8, 2)])
+def test_diag_fused_projection_and_fused_gradients(B, T, M, K):
+    """Forward scan with b_t = Bc x_{t-1} formed on the fly (segment path), then the reverse
+    scan of a random cotangent with dlam and dBc accumulated inside it; with and without the
+    adjoint itself stored."""
+    rng = np.random.default_rng(B * T + M + K)
+    lam = (rng.uniform(0.9, 0.999, M) * np.exp(1j * rng.uniform(0, np.pi / 10, M))).astype(np.complex64)
+    Bc = ((rng.standard_normal((M, K)) + 1j * rng.standard_normal((M, K))) / np.sqrt(2 * K)).astype(np.complex64)
+    x = rng.standard_normal((B, T + 1, K)).astype(np.float32)
+    m = {"kind": "diag_ssm", "lam": lam, "Bc": Bc}
+    say("deer_solve diag fused", B, T, M, K)
+    res = D.deer_solve(m, x, 0.0, 0)
+    h_ref = O.diag_scan(lam, O.diag_ssm_inputs({"Bc": Bc}, x))
+    assert rel_inf(_c(res["z"].cpu().numpy()), h_ref) < TOL
+    g = (rng.standard_normal((B, T, M)) + 1j * rng.standard_normal((B, T, M))).astype(np.complex64)
+    gt = torch.tensor(np.stack([g.real, g.imag], -1))
+    say("deer_adjoint diag fused grads", B, T, M, K)
+    out = D.deer_adjoint(m, x, res["z"], 0.0, 0, g=gt)
+    a_ref = O.diag_scan_reverse(lam, g)
+    assert rel_inf(_c(out["lam"].cpu().numpy()), a_ref) < TOL
+    gr = O.diag_ssm_param_grads(a_ref, h_ref, x)
+    dl = out["grads"]["lam"].cpu().numpy()
+    dB = out["grads"]["Bc"].cpu().numpy()
+    assert rel_inf(_c(dl), gr["lam"]) < TOL
+    assert rel_inf(_c(dB), gr["Bc"]) < TOL
+    out2 = D.deer_adjoint(m, x, res["z"], 0.0, 0, g=gt, want_lam=False)
+    assert out2["lam"] is None
+    assert np.array_equal(out2["grads"]["lam"].cpu().numpy(), dl)
+    assert np.array_equal(out2["grads"]["Bc"].cpu().numpy(), dB)

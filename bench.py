@@ -6,9 +6,10 @@ One step = one pass of the whole path over one batch of synthetic input:
                    carries, fix-up + max-norm test, until every sequence converged or the
                    fixed iteration count) followed by deer_adjoint (MSE seed, reverse scan
                    with transposed Jacobians, parameter-gradient reductions).
-  diagonal SSM:    deer_solve (fused input projection + forward complex scan) followed by
-                   deer_adjoint (reverse scan with conj(lambda) + dlambda / dBc reductions)
-                   on a fixed cotangent.
+  diagonal SSM:    deer_solve (fused input projection + forward complex scan), then
+                   deer_readout_loss (read-out MLP loss, its cotangent dL/dRe h and the
+                   read-out gradients), then deer_adjoint on that real cotangent (reverse scan
+                   with conj(lambda) + dlambda / dBc reductions).
 Inputs are resident in HBM before the timed region.  The value is DEER timesteps per
 second: sum over sequences of T x Newton updates, per second of the whole step.
 
@@ -44,9 +45,10 @@ def _plrnn_step(D, model, xd, c, ws_s, ws_a):
     return sum(res["iters"])
 
 
-def _diag_step(D, model, xd, c, ws_s, ws_a, g):
-    res = D.deer_solve(model, xd, 0.0, 0, ws=ws_s)
-    D.deer_adjoint(model, xd, res["z"], 0.0, 0, g=g, ws=ws_a)
+def _diag_step(D, model, readout, xd, c, ws_s, ws_r, ws_a, bufs):
+    res = D.deer_solve(model, xd, 0.0, 0, ws=ws_s, z=bufs["h"])
+    r = D.deer_readout_loss(readout, res["z"], xd, g=bufs["g"], ws=ws_r)
+    D.deer_adjoint(model, xd, res["z"], 0.0, 0, g=r["g"], ws=ws_a)
     return c.B
 
 
@@ -65,10 +67,12 @@ def kernel_work(c, steps, updates):
         return {
             # forward: b formed from x on the fly; the write pass stores y (8 B per element)
             "k_diag_seg_write": ("hbm", elems * 8 + xin),
-            # adjoint: cotangent and forward states read, adjoint written (24 B per element),
+            # adjoint: real cotangent (4 B) and forward states (8 B) read, adjoint written (8 B),
             # dlam / dBc accumulated on the way
-            "k_diag_scan_lb_grads": ("hbm", elems * 24 + xin),
-            "k_diag_scan_lb": ("hbm", elems * 16 + xin),
+            "k_diag_scan_lb_grads": ("hbm", elems * 20 + xin),
+            "k_diag_scan_lb": ("hbm", elems * 12 + xin),
+            # read-out: three [rows x 64] x [64 x 128] products (s, g, dWa) on the matrix cores
+            "k_readout": ("mfma", steps * B * T * 3 * 2.0 * M * c.params["Wa"].shape[0]),
         }
     out = {}
     if c.kind == "plrnn":
@@ -174,11 +178,12 @@ def main():
     xd = torch.tensor(c.x, device=dev)
     if c.kind == "diag_ssm":
         model = D._Model({"kind": "diag_ssm", "lam": c.params["lam"], "Bc": c.params["Bc"]})
+        readout = D._Readout({k: c.params[k] for k in ("Wa", "ca", "Wb", "cb")})
         ws_s = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_SOLVE))
         ws_a = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_ADJOINT))
-        gen = torch.Generator(device=dev).manual_seed(0)
-        g = torch.randn(c.B, c.T, c.M, 2, device=dev, generator=gen) * 1e-6
-        step = lambda: _diag_step(D, model, xd, c, ws_s, ws_a, g)          # noqa: E731
+        ws_r = D._workspace(D.deer_readout_workspace_bytes(readout, c.B, c.T, c.M))
+        bufs = {"h": torch.empty(c.B, c.T, c.M, 2, device=dev), "g": torch.empty(c.B, c.T, c.M, device=dev)}
+        step = lambda: _diag_step(D, model, readout, xd, c, ws_s, ws_r, ws_a, bufs)   # noqa: E731
     elif c.kind in ("plrnn", "shplrnn"):
         model = D._Model({"kind": c.kind, **c.params})
         ws_s = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_SOLVE))

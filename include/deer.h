@@ -158,6 +158,50 @@ int deer_adjoint(const deer_model *model, const deer_forcing *forcing, int B, in
                  const float *x, const float *z0, const float *z, const float *g,
                  float *lam, const deer_grads *grads, void *ws, size_t ws_bytes, void *stream);
 
+/* Layout of the cotangent g of deer_adjoint_ex. */
+enum { DEER_G_NATIVE = 0, DEER_G_REAL = 1 };
+
+/* deer_adjoint with an explicit cotangent layout.  DEER_G_NATIVE is deer_adjoint.
+ * DEER_G_REAL (DEER_DIAG_SSM only): g is [B,T,M] real, dL/dRe h with dL/dIm h = 0 -- the
+ * cotangent the read-out MLP supplies (deer_readout_loss), read at 4 bytes per element. */
+int deer_adjoint_ex(const deer_model *model, const deer_forcing *forcing, int B, int T,
+                    const float *x, const float *z0, const float *z, const float *g, int g_layout,
+                    float *lam, const deer_grads *grads, void *ws, size_t ws_bytes, void *stream);
+
+/* Read-out MLP of the diagonal SSM and its loss (linear-SSM appendix: the LSSM's
+ * observation model; the MSE of eq. mse_loss_series on its outputs):
+ *   s_t = Wa Re(h_t) + ca,  y_t = Wb relu(s_t) + cb,
+ *   L = sum_{b,t} ||y_t - x_t||^2 / (B No T), with h_t the state after input x_{t-1}
+ *       (0-based arrays: state row t is compared with x row t + 1).
+ * Sizes: M <= 64 state channels, H <= 128 hidden units, No <= 4 outputs (= input dim K). */
+typedef struct {
+    int H;              /* hidden units                                                     */
+    int n_out;          /* No: outputs, equal to the data dimension of x                    */
+    const float *Wa;    /* [H, M]                                                           */
+    const float *ca;    /* [H] or NULL (zero)                                               */
+    const float *Wb;    /* [No, H]                                                          */
+    const float *cb;    /* [No] or NULL (zero)                                              */
+} deer_readout;
+
+typedef struct {
+    float *Wa, *ca, *Wb, *cb;   /* gradient outputs (device, same shapes) or NULL to skip    */
+} deer_readout_grads;
+
+/* Workspace bytes deer_readout_loss needs. */
+size_t deer_readout_workspace_bytes(const deer_readout *readout, int B, int T, int M);
+
+/* Forward and backward pass of the read-out at the states h [B,T,M][2] (complex):
+ *   g     [B,T,M] out (required): dL/dRe h_t = Wa^T ((Wb^T dy_t) * 1[s_t > 0]),
+ *         dy_t = 2 (y_t - x_{t+1}) / (B No T); feed it to deer_adjoint_ex(DEER_G_REAL).
+ *   loss  device [1] out or NULL.
+ *   masks [B,T,ceil(H/32)] out or NULL: the ReLU decisions 1[s_t > 0] taken (bit j of word
+ *         w is hidden unit 32 w + j).
+ *   grads read-out parameter gradients or NULL (sums over all (b, t), reduced in float64).
+ * Fully asynchronous on `stream`. */
+int deer_readout_loss(const deer_readout *readout, int B, int T, int M, const float *h, const float *x,
+                      float *g, float *loss, uint32_t *masks, const deer_readout_grads *grads, void *ws,
+                      size_t ws_bytes, void *stream);
+
 /* Residual and forced Jacobians of a PLRNN kind at trajectory z (eq. GTF_residual; the
  * Jacobian of F in the model-setup appendix; eq. error_forcing_decomp):
  *   F     [B,T,M] out or NULL: F(z~_{t-1}).

@@ -447,21 +447,31 @@ def diag_ssm_readout(params: dict, h: np.ndarray) -> np.ndarray:
     return np.maximum(s, 0.0) @ np.asarray(params["Wb"], f64).T + np.asarray(params["cb"], f64)
 
 
-def diag_ssm_loss_and_seed(params: dict, h: np.ndarray, x: np.ndarray):
-    """MSE of the read-out against x_{1:T} and g = dL/dRe(h) (chain rule through the MLP)."""
+def diag_ssm_readout_preactivation(params: dict, h: np.ndarray) -> np.ndarray:
+    """s_t = Wa Re(h_t) + ca, the hidden pre-activation of the read-out."""
+    return np.real(h) @ np.asarray(params["Wa"], f64).T + np.asarray(params["ca"], f64)
+
+
+def diag_ssm_loss_and_seed(params: dict, h: np.ndarray, x: np.ndarray, mask=None):
+    """MSE of the read-out against x_{1:T} and g = dL/dRe(h) (chain rule through the MLP).
+
+    mask: optional boolean [B, T, H] of ReLU decisions to use instead of s > 0 (the
+    decisions another implementation took; relu(s) = s * mask and relu' = mask)."""
     x = np.asarray(x, f64)
     Bn, T, _ = h.shape
     No = x.shape[2]
     Wa = np.asarray(params["Wa"], f64)
     Wb = np.asarray(params["Wb"], f64)
-    s = np.real(h) @ Wa.T + np.asarray(params["ca"], f64)
-    y = np.maximum(s, 0.0) @ Wb.T + np.asarray(params["cb"], f64)
+    s = diag_ssm_readout_preactivation(params, h)
+    m = (s > 0.0) if mask is None else np.asarray(mask, bool)
+    a1 = s * m
+    y = a1 @ Wb.T + np.asarray(params["cb"], f64)
     err = y - x[:, 1:]
     loss = float((err ** 2).sum() / (Bn * No * T))
     dy = 2.0 / (Bn * No * T) * err
-    ds = (dy @ Wb) * (s > 0.0)
+    ds = (dy @ Wb) * m
     g = ds @ Wa
-    grads = {"Wb": np.einsum("bto,btk->ok", dy, np.maximum(s, 0.0), optimize=True), "cb": dy.sum(axis=(0, 1)),
+    grads = {"Wb": np.einsum("bto,btk->ok", dy, a1, optimize=True), "cb": dy.sum(axis=(0, 1)),
              "Wa": np.einsum("btk,btn->kn", ds, np.real(h), optimize=True), "ca": ds.sum(axis=(0, 1))}
     return loss, g, grads
 

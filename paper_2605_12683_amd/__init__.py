@@ -8,6 +8,7 @@ Model dictionaries use the paper's names:
   vanilla PLRNN  {"kind": "plrnn",   "A": [M], "W": [M,M], "h": [M]}
   shallow PLRNN  {"kind": "shplrnn", "A": [M], "W1": [M,L], "W2": [L,M], "h1": [M], "h2": [L]}
   diagonal SSM   {"kind": "diag_ssm", "lam": complex64 [M], "Bc": complex64 [M,K]}
+  its read-out   {"Wa": [H,M], "ca": [H], "Wb": [No,H], "cb": [No]}
 """
 from __future__ import annotations
 
@@ -18,8 +19,8 @@ import torch
 from . import _binding as _b
 from ._binding import DeerError, load  # noqa: F401
 
-__all__ = ["deer_solve", "deer_adjoint", "plrnn_jacobian", "deer_scan", "deer_workspace_bytes",
-           "deer_scan_workspace_bytes", "deer_status_string", "DeerError", "load"]
+__all__ = ["deer_solve", "deer_adjoint", "deer_readout_loss", "plrnn_jacobian", "deer_scan", "deer_workspace_bytes",
+           "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_status_string", "DeerError", "load"]
 
 _KINDS = {"plrnn": _b.DEER_PLRNN, "shplrnn": _b.DEER_SHPLRNN, "diag_ssm": _b.DEER_DIAG_SSM}
 _INITS = {"teacher": _b.DEER_INIT_TEACHER, "zero": _b.DEER_INIT_ZERO, "user": _b.DEER_INIT_USER}
@@ -77,6 +78,54 @@ def _model(model):
     return model if isinstance(model, _Model) else _Model(model)
 
 
+class _Readout:
+    """Device copies of the read-out MLP parameters plus the C struct."""
+
+    def __init__(self, params: dict):
+        self.t = {k: _dev(params[k]) for k in ("Wa", "Wb")}
+        self.t["ca"] = _dev(params.get("ca"))
+        self.t["cb"] = _dev(params.get("cb"))
+        self.H, self.M = self.t["Wa"].shape
+        self.No = self.t["Wb"].shape[0]
+        self.c = _b.deer_readout(self.H, self.No, _ptr(self.t["Wa"]), _ptr(self.t["ca"]), _ptr(self.t["Wb"]),
+                                 _ptr(self.t["cb"]))
+
+
+def _readout(r):
+    return r if isinstance(r, _Readout) else _Readout(r)
+
+
+def deer_readout_workspace_bytes(readout, B: int, T: int, M: int) -> int:
+    r = _readout(readout)
+    return int(load().deer_readout_workspace_bytes(ctypes.byref(r.c), B, T, M))
+
+
+def deer_readout_loss(readout, h, x, *, want_grads: bool = True, want_masks: bool = False, want_loss: bool = True,
+                      g=None, ws=None) -> dict:
+    """Read-out MLP forward + backward at the complex states h [B,T,M][2]: returns
+    dict(g = dL/dRe h [B,T,M], loss [1], masks, grads {Wa, ca, Wb, cb})."""
+    lib = load()
+    r = _readout(readout)
+    h = _dev(h)
+    x = _dev(x)
+    B, T, M = h.shape[:3]
+    out_g = torch.empty(B, T, M, device="cuda") if g is None else g
+    loss = torch.empty(1, device="cuda") if want_loss else None
+    masks = torch.empty(B, T, (r.H + 31) // 32, dtype=torch.int32, device="cuda") if want_masks else None
+    grads = {}
+    gs = None
+    if want_grads:
+        grads = {"Wa": torch.empty(r.H, M, device="cuda"), "ca": torch.empty(r.H, device="cuda"),
+                 "Wb": torch.empty(r.No, r.H, device="cuda"), "cb": torch.empty(r.No, device="cuda")}
+        gs = _b.deer_readout_grads(_ptr(grads["Wa"]), _ptr(grads["ca"]), _ptr(grads["Wb"]), _ptr(grads["cb"]))
+    if ws is None:
+        ws = _workspace(lib.deer_readout_workspace_bytes(ctypes.byref(r.c), B, T, M))
+    st = lib.deer_readout_loss(ctypes.byref(r.c), B, T, M, _ptr(h), _ptr(x), _ptr(out_g), _ptr(loss), _ptr(masks),
+                               ctypes.byref(gs) if gs is not None else None, _ptr(ws), ws.numel(), _stream())
+    _b._check(st, "deer_readout_loss")
+    return {"g": out_g, "loss": loss, "masks": masks, "grads": grads}
+
+
 def deer_status_string(status: int) -> str:
     return load().deer_status_string(status).decode()
 
@@ -132,13 +181,20 @@ def deer_solve(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1
 
 def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, want_lam: bool = True,
                  want_grads: bool = True, ws=None) -> dict:
-    """Adjoint scan lam = dL/dz and parameter gradients at trajectory z."""
+    """Adjoint scan lam = dL/dz and parameter gradients at trajectory z.  Diagonal SSM: g is
+    complex [B,T,M] (or [B,T,M,2] float) = dL/dRe h + i dL/dIm h, or a real float tensor
+    [B,T,M] = dL/dRe h (the read-out's cotangent)."""
     lib = load()
     m = _model(model)
     x = _dev(x)
     B, T1, _ = x.shape
     T = T1 - 1
     z = _dev(z)
+    g_layout = _b.DEER_G_NATIVE
+    if m.kind == "diag_ssm" and g is not None:
+        gt = g if isinstance(g, torch.Tensor) else torch.as_tensor(g)
+        if not gt.is_complex() and gt.dim() == 3:
+            g_layout = _b.DEER_G_REAL
     g = _dev(g)
     shape = (B, T, m.M, 2) if m.kind == "diag_ssm" else (B, T, m.M)
     lam = torch.empty(shape, device="cuda") if want_lam else None
@@ -162,8 +218,8 @@ def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, w
         ws = _workspace(lib.deer_workspace_bytes(ctypes.byref(m.c), B, T, _b.DEER_OP_ADJOINT))
     f = _b.deer_forcing(float(alpha), int(n_forced))
     z0d = _dev(z0)
-    st = lib.deer_adjoint(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(g), _ptr(lam),
-                          ctypes.byref(gs), _ptr(ws), ws.numel(), _stream())
+    st = lib.deer_adjoint_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(g),
+                             g_layout, _ptr(lam), ctypes.byref(gs), _ptr(ws), ws.numel(), _stream())
     _b._check(st, "deer_adjoint")
     return {"lam": lam, "grads": grads}
 

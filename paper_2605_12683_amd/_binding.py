@@ -19,10 +19,11 @@ DEER_PLRNN, DEER_SHPLRNN, DEER_DIAG_SSM = 0, 1, 2
 DEER_INIT_TEACHER, DEER_INIT_ZERO, DEER_INIT_USER = 0, 1, 2
 DEER_OP_SOLVE, DEER_OP_ADJOINT = 0, 1
 DEER_SCAN_DENSE, DEER_SCAN_DIAG_C64 = 0, 1
+DEER_G_NATIVE, DEER_G_REAL = 0, 1
 
-EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "plrnn_jacobian", "deer_scan",
-            "deer_scan_workspace_bytes", "deer_status_string", "deer_last_error", "deer_timing_enable",
-            "deer_timing_report"]
+EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "deer_adjoint_ex", "plrnn_jacobian", "deer_scan",
+            "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_readout_loss", "deer_status_string",
+            "deer_last_error", "deer_timing_enable", "deer_timing_report"]
 
 _fp = ctypes.c_void_p
 
@@ -43,6 +44,14 @@ class deer_solve_opts(ctypes.Structure):
 
 class deer_grads(ctypes.Structure):
     _fields_ = [("A", _fp), ("W", _fp), ("W2", _fp), ("h", _fp), ("h2", _fp)]
+
+
+class deer_readout(ctypes.Structure):
+    _fields_ = [("H", ctypes.c_int), ("n_out", ctypes.c_int), ("Wa", _fp), ("ca", _fp), ("Wb", _fp), ("cb", _fp)]
+
+
+class deer_readout_grads(ctypes.Structure):
+    _fields_ = [("Wa", _fp), ("ca", _fp), ("Wb", _fp), ("cb", _fp)]
 
 
 _lib = None
@@ -69,6 +78,14 @@ def load(path: str = LIB_PATH):
     lib.deer_adjoint.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, vp, P(deer_grads), vp, sz,
                                  vp]
     lib.deer_adjoint.restype = i32
+    lib.deer_adjoint_ex.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, i32, vp, P(deer_grads),
+                                    vp, sz, vp]
+    lib.deer_adjoint_ex.restype = i32
+    lib.deer_readout_workspace_bytes.argtypes = [P(deer_readout), i32, i32, i32]
+    lib.deer_readout_workspace_bytes.restype = sz
+    lib.deer_readout_loss.argtypes = [P(deer_readout), i32, i32, i32, vp, vp, vp, vp, vp, P(deer_readout_grads), vp,
+                                      sz, vp]
+    lib.deer_readout_loss.restype = i32
     lib.plrnn_jacobian.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.plrnn_jacobian.restype = i32
     lib.deer_scan.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]

@@ -647,7 +647,21 @@ int deer_solve(const deer_model *m, const deer_forcing *f, const deer_solve_opts
 int deer_adjoint(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
                  const float *z, const float *g, float *lam, const deer_grads *grads, void *ws, size_t ws_bytes,
                  void *stream) {
+    return deer_adjoint_ex(m, f, B, T, x, z0, z, g, DEER_G_NATIVE, lam, grads, ws, ws_bytes, stream);
+}
+
+int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
+                    const float *z, const float *g, int g_layout, float *lam, const deer_grads *grads, void *ws,
+                    size_t ws_bytes, void *stream) {
     set_error("");
+    if (g_layout != DEER_G_NATIVE && g_layout != DEER_G_REAL) {
+        set_error("unknown cotangent layout %d", g_layout);
+        return DEER_ERR_INVALID_ARG;
+    }
+    if (g_layout == DEER_G_REAL && m && m->kind != DEER_DIAG_SSM) {
+        set_error("DEER_G_REAL applies to DEER_DIAG_SSM only");
+        return DEER_ERR_INVALID_ARG;
+    }
     int rc = check_common(m, f, B, T);
     if (rc) return rc;
     if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
@@ -699,10 +713,39 @@ int deer_adjoint(const deer_model *m, const deer_forcing *f, int B, int T, const
         if ((rc = check_ws(ws, ws_bytes, diag_bytes(B, T, m->M, m->L, DEER_OP_ADJOINT)))) return rc;
         float *dlam = grads ? grads->A : nullptr, *dBc = grads ? grads->W : nullptr;
         if (!lam && !dlam && !dBc) return DEER_OK;
-        return launch_diag_adjoint(B, T, m->M, m->L, m->A, g, z, x, lam, dlam, dBc, ws, st);
+        return launch_diag_adjoint(B, T, m->M, m->L, m->A, g, g_layout == DEER_G_REAL, z, x, lam, dlam, dBc, ws, st);
     }
     set_error("deer_adjoint: model kind %d not supported yet", m->kind);
     return DEER_ERR_INVALID_ARG;
+}
+
+static int check_readout(const deer_readout *r, int B, int T, int M) {
+    if (!r || !r->Wa || !r->Wb) { set_error("read-out needs Wa and Wb"); return DEER_ERR_INVALID_ARG; }
+    if (B <= 0 || T <= 0) { set_error("B and T must be positive"); return DEER_ERR_INVALID_ARG; }
+    if (M <= 0 || M > 64) { set_error("read-out supports 1 <= M <= 64 (M=%d)", M); return DEER_ERR_INVALID_ARG; }
+    if (r->H <= 0 || r->H > 128) { set_error("read-out supports 1 <= H <= 128 (H=%d)", r->H); return DEER_ERR_INVALID_ARG; }
+    if (r->n_out <= 0 || r->n_out > 4) { set_error("read-out supports 1 <= n_out <= 4"); return DEER_ERR_INVALID_ARG; }
+    if ((long)B * (long)T > (1L << 31)) { set_error("B*T too large"); return DEER_ERR_INVALID_ARG; }
+    return DEER_OK;
+}
+
+size_t deer_readout_workspace_bytes(const deer_readout *r, int B, int T, int M) {
+    if (check_readout(r, B, T, M) != DEER_OK) return 0;
+    return readout_ws_bytes(B, T);
+}
+
+int deer_readout_loss(const deer_readout *r, int B, int T, int M, const float *h, const float *x, float *g,
+                      float *loss, uint32_t *masks, const deer_readout_grads *grads, void *ws, size_t ws_bytes,
+                      void *stream) {
+    set_error("");
+    int rc = check_readout(r, B, T, M);
+    if (rc) return rc;
+    if (!h || !x || !g) { set_error("h, x and g are required"); return DEER_ERR_INVALID_ARG; }
+    if ((rc = check_ws(ws, ws_bytes, readout_ws_bytes(B, T)))) return rc;
+    RoArgs ra{r->Wa, r->ca, r->Wb, r->cb, M, r->H, r->n_out};
+    RoGrads gr{grads ? grads->Wa : nullptr, grads ? grads->ca : nullptr, grads ? grads->Wb : nullptr,
+               grads ? grads->cb : nullptr};
+    return launch_readout(ra, B, T, h, x, g, masks, loss, gr, ws, (hipStream_t)stream);
 }
 
 int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, const float *b, float *y, void *ws,

@@ -165,7 +165,8 @@ __device__ __forceinline__ void pub_word(unsigned long long *p, float v) {
 // be null (the adjoint itself not stored).
 constexpr int DNV = 10;   // 2 + 2 K partial values per channel, K <= 4
 
-template <bool PROJ, bool GRADS>
+// GREAL: b is real [B,T,M] (imaginary part zero), read at 4 bytes per element.
+template <bool PROJ, bool GRADS, bool GREAL = false>
 __global__ __launch_bounds__(DNW * 64) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_diag_scan_lb(const float *__restrict__ lam, int conj_lam,
                                                           const float *__restrict__ bin, const float *__restrict__ Bc,
                                                           int K, const float *__restrict__ u, int rev, int B, int T,
@@ -221,7 +222,9 @@ __global__ __launch_bounds__(DNW * 64) __attribute__((amdgpu_waves_per_eu(4, 8))
         float2 v = make_float2(0.f, 0.f);
         if (mok && p < T) {
             const long tau = rev ? (T - 1 - p) : p;
-            if (!PROJ) {
+            if (!PROJ && GREAL) {
+                v = make_float2(__builtin_nontemporal_load(bin + ((long)b * T + tau) * M + m), 0.f);
+            } else if (!PROJ) {
                 const v2f t2 = __builtin_nontemporal_load(reinterpret_cast<const v2f *>(bin + (((long)b * T + tau) * M + m) * 2));
                 v = make_float2(t2.x, t2.y);
             } else {
@@ -773,8 +776,8 @@ size_t diag_adjoint_ws_bytes(int B, int T, int M, int K) {
 
 // Reverse scan of the cotangent g with the parameter gradients fused (dlam, dBc may be
 // null; lam_out may be null).
-int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const float *g, const float *h, const float *x,
-                        float *lam_out, float *dlam, float *dBc, void *ws, hipStream_t st) {
+int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const float *g, bool g_real, const float *h,
+                        const float *x, float *lam_out, float *dlam, float *dBc, void *ws, hipStream_t st) {
     const int ntile = (M + DTC - 1) / DTC;
     const int nq = (T + DCH - 1) / DCH;
     const int nblk = B * ntile * nq;
@@ -796,14 +799,14 @@ int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const floa
     const bool grads = dlam || dBc;
     {
         KTimer _kt(grads ? "k_diag_scan_lb_grads" : "k_diag_scan_lb", st);
-        if (grads)
-            hipLaunchKernelGGL((k_diag_scan_lb<false, true>), dim3(nblk), dim3(DNW * 64), 0, st, lam, 1, g,
-                               (const float *)nullptr, K, x, 1, B, T, M, ntile, nq, ticket, aggw, incw, lam_out, h,
-                               part);
-        else
-            hipLaunchKernelGGL((k_diag_scan_lb<false, false>), dim3(nblk), dim3(DNW * 64), 0, st, lam, 1, g,
-                               (const float *)nullptr, K, x, 1, B, T, M, ntile, nq, ticket, aggw, incw, lam_out,
-                               (const float *)nullptr, (float *)nullptr);
+#define LBA(GR, RE, HP, PP)                                                                                        \
+    hipLaunchKernelGGL((k_diag_scan_lb<false, GR, RE>), dim3(nblk), dim3(DNW * 64), 0, st, lam, 1, g,             \
+                       (const float *)nullptr, K, x, 1, B, T, M, ntile, nq, ticket, aggw, incw, lam_out, HP, PP)
+        if (grads && g_real) LBA(true, true, h, part);
+        else if (grads) LBA(true, false, h, part);
+        else if (g_real) LBA(false, true, (const float *)nullptr, (float *)nullptr);
+        else LBA(false, false, (const float *)nullptr, (float *)nullptr);
+#undef LBA
     }
     DEER_LAUNCH_CHECK("k_diag_scan_lb");
     if (grads) {

@@ -61,13 +61,25 @@ int launch_grads_shplrnn(const ShArgs &a, const float *z, const float *lam, cons
                          const deer_grads *gr, hipStream_t st);
 int launch_mse_seed(const float *z, const float *x, float scale, int B, int T, int M, int N, float *g, hipStream_t st);
 
+// read-out MLP of the diagonal SSM
+struct RoArgs {
+    const float *Wa, *ca, *Wb, *cb;
+    int M, H, No;
+};
+struct RoGrads {
+    float *Wa, *ca, *Wb, *cb;
+};
+size_t readout_ws_bytes(int B, int T);
+int launch_readout(const RoArgs &ra, int B, int T, const float *h, const float *x, float *g, uint32_t *masks,
+                   float *loss, const RoGrads &gr, void *ws, hipStream_t st);
+
 // diagonal complex scan
 size_t diag_scan_ws_bytes(int B, int T, int M);
 int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const float *b, const float *Bc, int K,
                      const float *u, float *y, void *ws, hipStream_t st);
 size_t diag_adjoint_ws_bytes(int B, int T, int M, int K);
-int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const float *g, const float *h, const float *x,
-                        float *lam_out, float *dlam, float *dBc, void *ws, hipStream_t st);
+int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const float *g, bool g_real, const float *h,
+                        const float *x, float *lam_out, float *dlam, float *dBc, void *ws, hipStream_t st);
 
 // small utilities
 int launch_fill_teacher(int B, int T, int M, int N, const float *x, float *z, hipStream_t st);

@@ -89,3 +89,70 @@ def test_diag_fused_projection_and_fused_gradients(B, T, M, K):
     assert out2["lam"] is None
     assert np.array_equal(out2["grads"]["lam"].cpu().numpy(), dl)
     assert np.array_equal(out2["grads"]["Bc"].cpu().numpy(), dB)
+
+
+def _readout_params(M, H, No, rng):
+    return {"Wa": (rng.standard_normal((H, M)) / np.sqrt(M)).astype(np.float32),
+            "ca": (0.1 * rng.standard_normal(H)).astype(np.float32),
+            "Wb": (rng.standard_normal((No, H)) / np.sqrt(H)).astype(np.float32),
+            "cb": (0.1 * rng.standard_normal(No)).astype(np.float32)}
+
+
+def _bits(words, H):
+    w = words.astype(np.uint32)
+    bits = (w[..., :, None] >> np.arange(32, dtype=np.uint32)) & 1
+    return bits.reshape(w.shape[:-1] + (-1,))[..., :H].astype(bool)
+
+
+@pytest.mark.parametrize("B,T,M,H,No", [(1, 1, 1, 1, 1), (2, 37, 64, 128, 3), (1, 1000, 17, 50, 2),
+                                        (3, 5000, 64, 128, 4), (2, 300, 64, 16, 3), (1, 70, 40, 100, 1)])
+def test_readout_loss_g_and_grads(B, T, M, H, No):
+    """Read-out MLP on the matrix cores: the ReLU decisions equal the float64 ones outside a
+    tie band; loss, g = dL/dRe h and the read-out gradients equal the float64 oracle taken
+    with the GPU's decisions."""
+    rng = np.random.default_rng(B * T + M + H + No)
+    prm = _readout_params(M, H, No, rng)
+    h = (rng.standard_normal((B, T, M)) + 1j * rng.standard_normal((B, T, M))).astype(np.complex64)
+    x = rng.standard_normal((B, T + 1, No)).astype(np.float32)
+    say("deer_readout_loss", B, T, M, H, No)
+    out = D.deer_readout_loss(prm, torch.tensor(h), x, want_masks=True)
+    got = _bits(out["masks"].cpu().numpy(), H)
+    s = O.diag_ssm_readout_preactivation(prm, h)
+    far = np.abs(s) > 1e-5 * max(np.abs(s).max(), 1e-30)
+    assert np.array_equal(got[far], (s > 0)[far])
+    loss, g, gr = O.diag_ssm_loss_and_seed(prm, h, x, mask=got)
+    assert abs(float(out["loss"].cpu()[0]) - loss) <= 1e-5 * abs(loss)
+    assert rel_inf(out["g"].cpu().numpy(), g) < TOL
+    for k in ("Wa", "ca", "Wb", "cb"):
+        assert rel_inf(out["grads"][k].cpu().numpy(), gr[k]) < TOL, k
+    # without gradients / masks / loss the cotangent is bit-identical
+    out2 = D.deer_readout_loss(prm, torch.tensor(h), x, want_grads=False, want_loss=False)
+    assert np.array_equal(out2["g"].cpu().numpy(), out["g"].cpu().numpy())
+
+
+def test_diag_training_step_with_readout():
+    """Workload-4 model at reduced T, the whole step: forward scan with the fused projection,
+    read-out loss and cotangent, reverse scan of the real cotangent with dlam, dBc."""
+    c = W.make_config(4, B=2, T=3000)
+    p = c.params
+    m = {"kind": "diag_ssm", "lam": p["lam"], "Bc": p["Bc"]}
+    ro = {k: p[k] for k in ("Wa", "ca", "Wb", "cb")}
+    say("diag step: solve")
+    res = D.deer_solve(m, c.x, 0.0, 0)
+    say("diag step: read-out")
+    r = D.deer_readout_loss(ro, res["z"], c.x, want_masks=True)
+    say("diag step: adjoint (real g)")
+    out = D.deer_adjoint(m, c.x, res["z"], 0.0, 0, g=r["g"])
+    h = O.diag_scan(p["lam"], O.diag_ssm_inputs(p, c.x))
+    assert rel_inf(_c(res["z"].cpu().numpy()), h) < TOL
+    mask = _bits(r["masks"].cpu().numpy(), p["Wa"].shape[0])
+    loss, g, gr = O.diag_ssm_loss_and_seed(p, h, c.x, mask=mask)
+    assert abs(float(r["loss"].cpu()[0]) - loss) <= 1e-5 * loss
+    assert rel_inf(r["g"].cpu().numpy(), g) < TOL
+    a = O.diag_scan_reverse(p["lam"], g.astype(np.complex128))
+    assert rel_inf(_c(out["lam"].cpu().numpy()), a) < TOL
+    pg = O.diag_ssm_param_grads(a, h, c.x)
+    assert rel_inf(_c(out["grads"]["lam"].cpu().numpy()), pg["lam"]) < TOL
+    assert rel_inf(_c(out["grads"]["Bc"].cpu().numpy()), pg["Bc"]) < TOL
+    for k in ("Wa", "ca", "Wb", "cb"):
+        assert rel_inf(r["grads"][k].cpu().numpy(), gr[k]) < TOL, k

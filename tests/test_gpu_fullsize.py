@@ -69,31 +69,48 @@ def test_plrnn_workload_full(cfg):
 
 
 def test_diag_workload_full():
-    """Workload 4: fused-projection forward scan, reverse scan of a seeded cotangent, and
-    dlambda / dBc, against the complex128 oracle."""
+    """Workload 4, the step bench.py times: fused-projection forward scan, read-out loss and
+    cotangent (ReLU decisions taken from the GPU, checked against float64 outside a tie
+    band), reverse scan of the real cotangent with dlambda / dBc, against the oracle."""
     _blas_threads()
     c = W.make_config(4)
     p = c.params
     m = {"kind": "diag_ssm", "lam": p["lam"], "Bc": p["Bc"]}
+    ro = {k: p[k] for k in ("Wa", "ca", "Wb", "cb")}
     say("deer_solve diag full")
     res = D.deer_solve(m, c.x, 0.0, 0)
     h_gpu = res["z"]
-    b = O.diag_ssm_inputs(p, c.x)
-    h = O.diag_scan(p["lam"], b)
-    del b
+    say("deer_readout_loss diag full")
+    r = D.deer_readout_loss(ro, h_gpu, c.x, want_masks=True)
+    say("deer_adjoint diag full (real g)")
+    out = D.deer_adjoint(m, c.x, h_gpu, 0.0, 0, g=r["g"])
+    h = O.diag_scan(p["lam"], O.diag_ssm_inputs(p, c.x))
     hg = h_gpu.cpu().numpy()
     assert rel_inf(hg[..., 0] + 1j * hg[..., 1], h) < TOL
     del hg
-    rng = np.random.default_rng(4242)
-    g = (rng.standard_normal(h.shape) + 1j * rng.standard_normal(h.shape)).astype(np.complex64)
-    say("deer_adjoint diag full")
-    out = D.deer_adjoint(m, c.x, h_gpu, 0.0, 0, g=torch.tensor(g))
-    ag = out["lam"].cpu().numpy()
+    H = p["Wa"].shape[0]
+    w = r["masks"].cpu().numpy().astype(np.uint32)
+    mask = (((w[..., :, None] >> np.arange(32, dtype=np.uint32)) & 1).reshape(w.shape[:-1] + (-1,))[..., :H]
+            .astype(bool))
+    del w
+    s = O.diag_ssm_readout_preactivation(p, h)
+    far = np.abs(s) > 1e-5 * np.abs(s).max()
+    assert np.array_equal(mask[far], (s > 0)[far])
+    print(f"[gpu-case] read-out in-band ties: {(~far).sum()} of {far.size}", flush=True)
+    del s, far
+    loss, g, gr = O.diag_ssm_loss_and_seed(p, h, c.x, mask=mask)
+    del mask
+    assert abs(float(r["loss"].cpu()[0]) - loss) <= 1e-5 * loss
+    assert rel_inf(r["g"].cpu().numpy(), g) < TOL
+    for k in ("Wa", "ca", "Wb", "cb"):
+        assert rel_inf(r["grads"][k].cpu().numpy(), gr[k]) < TOL, k
     a = O.diag_scan_reverse(p["lam"], g)
+    del g
+    ag = out["lam"].cpu().numpy()
     assert rel_inf(ag[..., 0] + 1j * ag[..., 1], a) < TOL
     del ag
-    gr = O.diag_ssm_param_grads(a, h, c.x)
+    pg = O.diag_ssm_param_grads(a, h, c.x)
     dl = out["grads"]["lam"].cpu().numpy()
     dB = out["grads"]["Bc"].cpu().numpy()
-    assert rel_inf(dl[..., 0] + 1j * dl[..., 1], gr["lam"]) < TOL
-    assert rel_inf(dB[..., 0] + 1j * dB[..., 1], gr["Bc"]) < TOL
+    assert rel_inf(dl[..., 0] + 1j * dl[..., 1], pg["lam"]) < TOL
+    assert rel_inf(dB[..., 0] + 1j * dB[..., 1], pg["Bc"]) < TOL

@@ -466,3 +466,31 @@ def test_diag_ssm_gradients_match_autograd():
     assert np.allclose(G["Bc"], br.grad.numpy() + 1j * bi.grad.numpy(), rtol=1e-9, atol=1e-13)
     for k, v in [("Wa", Wa), ("ca", ca), ("Wb", Wb), ("cb", cb)]:
         assert np.allclose(G[k], v.grad.numpy(), rtol=1e-9, atol=1e-13), k
+
+
+def test_readout_with_given_masks_matches_autograd():
+    """The mask-conditioned read-out (ReLU decisions supplied from outside, as the GPU parity
+    tests do) equals torch autograd of y = Wb (s * m) + cb with that fixed mask m, for a
+    random mask; with m = (s > 0) it reproduces the plain read-out."""
+    from workloads import diag_ssm_params
+    prm = diag_ssm_params(5, 2, 7, 2, np.random.default_rng(80))
+    rng = np.random.default_rng(81)
+    h = rng.standard_normal((2, 9, 5)) + 1j * rng.standard_normal((2, 9, 5))
+    x = _x(2, 9, 2, 82)
+    s = O.diag_ssm_readout_preactivation(prm, h)
+    base = O.diag_ssm_loss_and_seed(prm, h, x)
+    own = O.diag_ssm_loss_and_seed(prm, h, x, mask=s > 0)
+    assert base[0] == own[0] and np.array_equal(base[1], own[1])
+    m = rng.random(s.shape) < 0.5
+    loss, g, gr = O.diag_ssm_loss_and_seed(prm, h, x, mask=m)
+    t = lambda a: torch.tensor(np.asarray(a, np.float64), requires_grad=True)
+    hr = t(h.real)
+    Wa, ca, Wb, cb = t(prm["Wa"]), t(prm["ca"]), t(prm["Wb"]), t(prm["cb"])
+    st = hr @ Wa.T + ca
+    y = (st * torch.tensor(m, dtype=torch.float64)) @ Wb.T + cb
+    L = ((y - torch.tensor(x[:, 1:].astype(np.float64))) ** 2).sum() / (2 * 2 * 9)
+    L.backward()
+    assert np.isclose(loss, float(L.detach()), rtol=1e-12)
+    assert np.allclose(g, hr.grad.numpy(), rtol=1e-10, atol=1e-14)
+    for k, v in [("Wa", Wa), ("ca", ca), ("Wb", Wb), ("cb", cb)]:
+        assert np.allclose(gr[k], v.grad.numpy(), rtol=1e-10, atol=1e-14), k

@@ -74,6 +74,15 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 
 // forced input of step s (array index) for latent i:
 //   s == 0: z0 (or [x_0; 0] when z0 is null);  s >= 1: fl(fl(p*z_{s-1}) + fl(a*zbar_s))
+// Workgroup barrier that orders LDS only: unlike __syncthreads it does not wait for
+// outstanding global loads, so loads issued ahead (prefetch) stay in flight across it.  For
+// kernels whose threads exchange data through LDS alone.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ float forced_state(const float *__restrict__ x, const float *__restrict__ z0,
                                               const float *__restrict__ z, int b, int s, int i, int T, int M,
                                               int N, float alpha) {

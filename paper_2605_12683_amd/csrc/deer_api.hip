@@ -143,7 +143,8 @@ static int chunk_override() {
 }
 
 // Chunk length of the dense scans: enough chains to fill the machine (about 2048 waves),
-// at most 128 chunks per sequence so that the serial carry pass stays short.
+// and a bounded number of chunks per sequence so that the carry pass stays short: 128 with
+// the single-level carry (MP = 64), 1024 with the two-level carry (MP <= 32).
 static int choose_chunk(int B, int T, int MP) {
     const int ov = chunk_override();
     if (ov > 0) return ov < T ? ov : T;
@@ -151,7 +152,8 @@ static int choose_chunk(int B, int T, int MP) {
     const long target_chains = 2048L * (64 / MP);
     long C = (total + target_chains - 1) / target_chains;
     if (C < 16) C = 16;
-    const long minC = (T + 127) / 128;
+    const long maxc = MP <= 32 ? 1024 : 128;
+    const long minC = (T + maxc - 1) / maxc;
     if (C < minC) C = minC;
     if (C > T) C = T;
     return (int)C;
@@ -164,15 +166,17 @@ struct NewtonCtl {
     int *active;
     float *gamma;
     uint32_t *norm_bits;
-    float *zalt;   // second iterate buffer [B,T,M]
+    uint32_t *chain_bits;   // per-chain maxima [2][B * ncs] before the per-sequence reduction
+    float *zalt;            // second iterate buffer [B,T,M]
 };
 
-static NewtonCtl carve_ctl(Carver &c, int B, size_t seq_elems) {
+static NewtonCtl carve_ctl(Carver &c, int B, size_t seq_elems, size_t nchains) {
     NewtonCtl n{};
     uint32_t *blk = c.take<uint32_t>(2 * (size_t)B);
     n.active = (int *)blk;
     n.gamma = blk ? (float *)(blk + B) : nullptr;
     n.norm_bits = c.take<uint32_t>(2 * (size_t)B);
+    n.chain_bits = c.take<uint32_t>(2 * nchains);
     n.zalt = c.take<float>((size_t)B * seq_elems);
     return n;
 }
@@ -180,7 +184,7 @@ static NewtonCtl carve_ctl(Carver &c, int B, size_t seq_elems) {
 struct PlrnnWs {
     float *r;
     uint32_t *masks;
-    float *P, *v, *carry;
+    float *P, *v, *carry, *gws;
     NewtonCtl ctl;
     float *gpart;
     double *gpart2;
@@ -199,8 +203,9 @@ static PlrnnWs carve_plrnn(void *ws, int B, int T, int M, int op, size_t *bytes)
     w.P = c.take<float>(nch * w.MP * w.MP);
     w.v = c.take<float>(nch * w.MP);
     w.carry = c.take<float>(nch * w.MP);
+    w.gws = c.take<float>(carry_ws_floats(w.MP, B, w.ncs));
     if (op == DEER_OP_SOLVE) {
-        w.ctl = carve_ctl(c, B, (size_t)T * M);
+        w.ctl = carve_ctl(c, B, (size_t)T * M, nch);
         w.r = c.take<float>((size_t)B * T * M);
     } else {
         w.gpart = c.take<float>(nch * w.MP * (w.MP + 2));
@@ -211,7 +216,7 @@ static PlrnnWs carve_plrnn(void *ws, int B, int T, int M, int op, size_t *bytes)
 }
 
 struct DenseWs {
-    float *P, *v, *carry;
+    float *P, *v, *carry, *gws;
     int C, ncs, MP;
 };
 
@@ -225,6 +230,7 @@ static DenseWs carve_dense(void *ws, int B, int T, int M, size_t *bytes) {
     w.P = c.take<float>(nch * w.MP * w.MP);
     w.v = c.take<float>(nch * w.MP);
     w.carry = c.take<float>(nch * w.MP);
+    w.gws = c.take<float>(carry_ws_floats(w.MP, B, w.ncs));
     *bytes = c.off;
     return w;
 }
@@ -243,7 +249,8 @@ static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, 
     w.masks = c.take<uint32_t>((size_t)B * T * LW);
     w.J = c.take<float>((size_t)B * T * M * M);
     if (op == DEER_OP_SOLVE) {
-        w.ctl = carve_ctl(c, B, (size_t)T * M);
+        const int C = choose_chunk(B, T, padded_dim(M));
+        w.ctl = carve_ctl(c, B, (size_t)T * M, (size_t)B * ((T + C - 1) / C));
         w.r = c.take<float>((size_t)B * T * M);
     } else {
         if (need_g) w.g = c.take<float>((size_t)B * T * M);
@@ -467,8 +474,9 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     auto update = [&](const int *dact, const float *gam, const float *zin, float *zout) -> int {
         int r;
         if ((r = launch_newton_product_plrnn(a, zin, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, st))) return r;
-        if ((r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, nbits, B, w.ncs, st))) return r;
-        return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, zin, zout, nbits, dact, gam, w.C, w.ncs, st);
+        if ((r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, nbits, B, w.ncs, w.gws, st))) return r;
+        return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, zin, zout, w.ctl.chain_bits, nbits, dact, gam, w.C,
+                                      w.ncs, st);
     };
     if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
@@ -498,8 +506,9 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
         if ((r = launch_resjac_shplrnn(a, zin, nullptr, w.r, w.masks, dact, st))) return r;
         if ((r = launch_jacform_shplrnn(a, w.masks, w.J, dact, gam, st))) return r;
         if ((r = launch_chunk_product_dense(false, B, T, m->M, w.J, w.r, -1.f, d.P, d.v, dact, d.C, d.ncs, st))) return r;
-        if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nbits, B, d.ncs, st))) return r;
-        return launch_fixup_dense(0, B, T, m->M, w.J, w.r, -1.f, d.carry, zin, zout, nbits, dact, d.C, d.ncs, st);
+        if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nbits, B, d.ncs, d.gws, st))) return r;
+        return launch_fixup_dense(0, B, T, m->M, w.J, w.r, -1.f, d.carry, zin, zout, w.ctl.chain_bits, nbits, dact,
+                                  d.C, d.ncs, st);
     };
     if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
@@ -676,7 +685,7 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
         if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, w.masks, nullptr, st))) return rc;
         if ((rc = launch_chunk_product_plrnn(a, true, w.masks, g, z, scale, w.P, w.v, nullptr, w.C, w.ncs, st)))
             return rc;
-        if ((rc = launch_carry(w.MP, true, w.P, w.v, w.carry, nullptr, nullptr, B, w.ncs, st))) return rc;
+        if ((rc = launch_carry(w.MP, true, w.P, w.v, w.carry, nullptr, nullptr, B, w.ncs, w.gws, st))) return rc;
         if ((rc = launch_fixup_rev_plrnn(a, w.masks, g, scale, z, w.carry, lam, w.gpart, w.C, w.ncs, st))) return rc;
         if (grads && (grads->A || grads->W || grads->h)) {
             if ((rc = launch_reduce_gpart(w.gpart, B * w.ncs, w.MP, m->M, grads->A, grads->W, grads->h, w.gpart2, st))) return rc;
@@ -701,8 +710,8 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
         if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, w.masks, nullptr, st))) return rc;
         if ((rc = launch_jacform_shplrnn(a, w.masks, w.J, nullptr, nullptr, st))) return rc;
         if ((rc = launch_chunk_product_dense(true, B, T, m->M, w.J, gg, 1.f, d.P, d.v, nullptr, d.C, d.ncs, st))) return rc;
-        if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, st))) return rc;
-        if ((rc = launch_fixup_dense(2, B, T, m->M, w.J, gg, 1.f, d.carry, nullptr, lo, nullptr, nullptr, d.C, d.ncs, st))) return rc;
+        if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, d.gws, st))) return rc;
+        if ((rc = launch_fixup_dense(2, B, T, m->M, w.J, gg, 1.f, d.carry, nullptr, lo, nullptr, nullptr, nullptr, d.C, d.ncs, st))) return rc;
         if (grads && (grads->A || grads->W || grads->W2 || grads->h || grads->h2)) {
             if ((rc = launch_grads_shplrnn(a, z, lo, w.masks, w.part, grads, st))) return rc;
         }
@@ -769,8 +778,8 @@ int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, cons
         DenseWs w = carve_dense(ws, B, T, M, &need);
         const bool rev = reverse != 0;
         if ((rc = launch_chunk_product_dense(rev, B, T, M, J, b, 1.f, w.P, w.v, nullptr, w.C, w.ncs, st))) return rc;
-        if ((rc = launch_carry(w.MP, rev, w.P, w.v, w.carry, nullptr, nullptr, B, w.ncs, st))) return rc;
-        return launch_fixup_dense(rev ? 2 : 1, B, T, M, J, b, 1.f, w.carry, nullptr, y, nullptr, nullptr, w.C, w.ncs, st);
+        if ((rc = launch_carry(w.MP, rev, w.P, w.v, w.carry, nullptr, nullptr, B, w.ncs, w.gws, st))) return rc;
+        return launch_fixup_dense(rev ? 2 : 1, B, T, M, J, b, 1.f, w.carry, nullptr, y, nullptr, nullptr, nullptr, w.C, w.ncs, st);
     }
     set_error("deer_scan: unknown layout %d", layout);
     return DEER_ERR_INVALID_ARG;

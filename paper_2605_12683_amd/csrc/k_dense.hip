@@ -105,26 +105,26 @@ __global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restr
         if (!REV) {
             const int s = ulo + t;
             lds[lane] = u;
-            __syncthreads();
+            lds_barrier();
             float y = 0.f;
             if (run && ui < M) {
                 const float *Jr = J + (((size_t)ub * T + s) * M + ui) * M;
                 const float *l = lds + un * MP;
                 for (int k = 0; k < M; ++k) y = fmaf(Jr[k], l[k], y);
             }
-            __syncthreads();
+            lds_barrier();
             if (run && ui < M) u = fmaf(rhs_sign, rhs[((size_t)ub * T + s) * M + ui], y);
         } else {
             const int k = uhi - 1 - t;        // y_k = J_{k+1}^T y_{k+1} + b_k
             lds[lane] = u;
-            __syncthreads();
+            lds_barrier();
             float y = 0.f;
             if (run && ui < M && t > 0) {
                 const float *Jc = J + ((size_t)ub * T + k + 1) * M * M + ui;
                 const float *l = lds + un * MP;
                 for (int r = 0; r < M; ++r) y = fmaf(Jc[(size_t)r * M], l[r], y);
             }
-            __syncthreads();
+            lds_barrier();
             if (run && ui < M) u = fmaf(rhs_sign, rhs[((size_t)ub * T + k) * M + ui], y);
         }
     }
@@ -154,7 +154,7 @@ __global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restr
 template <int MP, int MODE>
 __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J, const float *__restrict__ rhs,
                                                     float rhs_sign, const float *__restrict__ carry_in,
-                                                    const float *zin, float *out, uint32_t *__restrict__ norm_bits,
+                                                    const float *zin, float *out, uint32_t *__restrict__ chain_bits,
                                                     const int *__restrict__ active, int B, int T, int M, int C,
                                                     int ncs) {
     using G = DGeo<MP>;
@@ -168,28 +168,61 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
     float y = (ok && i < M) ? carry_in[(size_t)id * MP + i] : 0.f;
     uint32_t emax = 0u, zmax = 0u;
     const int maxlen = __builtin_amdgcn_readfirstlane(C);
+    // the row (column, reverse) of J~ a step uses, its right-hand side and the iterate are
+    // loaded one step ahead
+    auto fetch = [&](int t, float *jv, float &bv, float &zv) {
+        const int k = MODE == 2 ? s1 - 1 - t : s0 + t;
+        const bool run = (MODE == 2 ? k >= s0 : k < s1) && i < M;
+        const size_t e = ((size_t)b * T + k) * M + i;
+        if (MODE != 2) {
+            const float *Jr = J + (((size_t)b * T + k) * M + i) * M;
+            if ((M & 3) == 0) {   // 16-byte aligned rows: vector loads
+                const float4 *J4 = reinterpret_cast<const float4 *>(Jr);
+#pragma unroll
+                for (int q = 0; q < MP / 4; ++q) {
+                    const float4 v4 = (run && 4 * q < M) ? J4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+                    jv[4 * q] = v4.x;
+                    jv[4 * q + 1] = v4.y;
+                    jv[4 * q + 2] = v4.z;
+                    jv[4 * q + 3] = v4.w;
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < MP; ++q) jv[q] = (run && q < M) ? Jr[q] : 0.f;
+            }
+        } else {
+            const bool has = run && k + 1 < T;
+            const float *Jc = J + ((size_t)b * T + k + 1) * M * M + i;
+#pragma unroll
+            for (int q = 0; q < MP; ++q) jv[q] = (has && q < M) ? Jc[(size_t)q * M] : 0.f;
+        }
+        bv = run ? rhs[e] : 0.f;
+        zv = (MODE == 0 && run) ? zin[e] : 0.f;
+    };
+    float jn[MP], bn, zn;
+    fetch(0, jn, bn, zn);
     for (int t = 0; t < maxlen; ++t) {
         const int k = MODE == 2 ? s1 - 1 - t : s0 + t;
         const bool run = (MODE == 2 ? k >= s0 : k < s1) && i < M;
+        float jc[MP];
+#pragma unroll
+        for (int q = 0; q < MP; ++q) jc[q] = jn[q];
+        const float bc = bn, zc = zn;
+        fetch(t + 1, jn, bn, zn);
         lds[lane] = y;
-        __syncthreads();
+        lds_barrier();
         float acc = 0.f;
-        if (run) {
+        {
             const float *l = lds + n * MP;
-            if (MODE != 2) {
-                const float *Jr = J + (((size_t)b * T + k) * M + i) * M;
-                for (int q = 0; q < M; ++q) acc = fmaf(Jr[q], l[q], acc);
-            } else if (k + 1 < T) {
-                const float *Jc = J + ((size_t)b * T + k + 1) * M * M + i;
-                for (int r = 0; r < M; ++r) acc = fmaf(Jc[(size_t)r * M], l[r], acc);
-            }
+#pragma unroll
+            for (int q = 0; q < MP; ++q) acc = fmaf(jc[q], l[q], acc);
         }
-        __syncthreads();
+        lds_barrier();
         if (run) {
             const size_t e = ((size_t)b * T + k) * M + i;
-            y = fmaf(rhs_sign, rhs[e], acc);
+            y = fmaf(rhs_sign, bc, acc);
             if (MODE == 0) {
-                const float zo = zin[e];
+                const float zo = zc;
                 out[e] = zo + y;
                 const uint32_t ab = abs_bits(y), zb = abs_bits(zo);
                 emax = emax > ab ? emax : ab;
@@ -207,9 +240,9 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
             emax = emax > o ? emax : o;
             zmax = zmax > oz ? zmax : oz;
         }
-        if (ok && i == 0) {
-            atomicMax(norm_bits + b, emax);
-            atomicMax(norm_bits + B + b, zmax);
+        if (ok && i == 0) {   // per-chain maxima, reduced per sequence by k_seq_max
+            chain_bits[id] = emax;
+            chain_bits[(size_t)B * ncs + id] = zmax;
         }
     }
 }
@@ -234,21 +267,22 @@ int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, co
 }
 
 int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
-                       const float *carry_in, const float *zin, float *out, uint32_t *norm_bits, const int *active,
-                       int C, int ncs, hipStream_t st) {
+                       const float *carry_in, const float *zin, float *out, uint32_t *chain_bits, uint32_t *norm_bits,
+                       const int *active, int C, int ncs, hipStream_t st) {
     const int MP = padded_dim(M);
     const int nch = B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt(mode == 2 ? "k_fixup_dense_rev" : "k_fixup_dense_fwd", st);
 #define FXD(MPV, MO)                                                                                          \
     hipLaunchKernelGGL((k_fixup_dense<MPV, MO>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, carry_in, zin, \
-                       out, norm_bits, active, B, T, M, C, ncs)
+                       out, chain_bits, active, B, T, M, C, ncs)
 #define FXD3(MO) \
     if (MP == 16) FXD(16, MO); else if (MP == 32) FXD(32, MO); else FXD(64, MO);
     if (mode == 0) { FXD3(0) } else if (mode == 1) { FXD3(1) } else { FXD3(2) }
 #undef FXD3
 #undef FXD
     DEER_LAUNCH_CHECK("k_fixup_dense");
+    if (mode == 0) return launch_seq_max(chain_bits, active, norm_bits, B, ncs, st);
     return DEER_OK;
 }
 

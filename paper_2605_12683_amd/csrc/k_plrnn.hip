@@ -91,7 +91,7 @@ __global__ __launch_bounds__(64) void k_resjac_plrnn(const float *__restrict__ A
             bal[q] = __ballot(pos);
             lds[q][lane] = pos ? zt[q] : 0.f;
         }
-        __syncthreads();
+        lds_barrier();
         float F[NG];
 #pragma unroll
         for (int q = 0; q < NG; ++q) {
@@ -99,7 +99,7 @@ __global__ __launch_bounds__(64) void k_resjac_plrnn(const float *__restrict__ A
             __builtin_amdgcn_sched_barrier(0);   // one dot product at a time: keeps the LDS reads of
                                                  // the other groups from being hoisted into registers
         }
-        __syncthreads();
+        lds_barrier();
 #pragma unroll
         for (int q = 0; q < NG; ++q) {
             const long row = rowv[q];
@@ -260,16 +260,16 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn(
             float w = 0.f;
             if (run && ui < M) w = mask_bit(masks, step, MW, ui) ? u : 0.f;
             lds[lane] = w;
-            __syncthreads();
+            lds_barrier();
             const float y = fmaf(du, u, lds_dot<MP>(lds, un, wv));
-            __syncthreads();
+            lds_barrier();
             if (run && ui < M) u = y - rhs[step * M + ui];
         } else {
             const int k = uhi - 1 - t;    // lam_k = J~_{k+1}^T lam_{k+1} + g_k
             lds[lane] = u;
-            __syncthreads();
+            lds_barrier();
             const float wt = lds_dot<MP>(lds, un, wv);
-            __syncthreads();
+            lds_barrier();
             if (run && ui < M) {
                 const size_t step = (size_t)ub * T + k;
                 float y = 0.f;
@@ -401,20 +401,29 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
         else zprev = z[((size_t)ub * T + us0 - 1) * M + ui];
     }
     float u = 0.f;
-    // prefetch of step 0
-    float zcur_n = 0.f, xb_n = 0.f;
-    if (ulen > 0 && lat) {
-        zcur_n = z[((size_t)ub * T + us0) * M + ui];
-        if (forced) xb_n = x[((size_t)ub * (T + 1) + us0) * N + ui];
-    }
+    // z_s and x_s are loaded PD steps ahead (a queue shifted by one every step)
+    constexpr int PD = 1;
+    float zq[PD], xq[PD];
+    auto fetch = [&](int t, float &zv, float &xv) {
+        zv = 0.f;
+        xv = 0.f;
+        if (t < ulen && lat) {
+            zv = z[((size_t)ub * T + us0 + t) * M + ui];
+            if (forced) xv = x[((size_t)ub * (T + 1) + us0 + t) * N + ui];
+        }
+    };
+#pragma unroll
+    for (int q = 0; q < PD; ++q) fetch(q, zq[q], xq[q]);
     for (int t = 0; t < maxlen; ++t) {
         const bool run = t < ulen && lat;
         const int s = us0 + t;
-        const float zcur = zcur_n, xb = xb_n;
-        if (t + 1 < ulen && lat) {
-            zcur_n = z[((size_t)ub * T + s + 1) * M + ui];
-            if (forced) xb_n = x[((size_t)ub * (T + 1) + s + 1) * N + ui];
+        const float zcur = zq[0], xb = xq[0];
+#pragma unroll
+        for (int q = 0; q + 1 < PD; ++q) {
+            zq[q] = zq[q + 1];
+            xq[q] = xq[q + 1];
         }
+        fetch(t + PD, zq[PD - 1], xq[PD - 1]);
         // forced state of this step (s == 0: z_0 itself)
         float zt = 0.f;
         if (run) {
@@ -424,9 +433,9 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
         const bool pos = zt > 0.f;
         const uint64_t bal = __ballot(pos);
         lds[lane] = pos ? zt : 0.f;
-        __syncthreads();
+        lds_barrier();
         const float F = fmaf(Ai, zt, lds_dot<MP>(lds, un, wrow)) + hi;
-        __syncthreads();
+        lds_barrier();
         const float r = zcur - F;
         if (run) {
             const size_t e = ((size_t)ub * T + s) * M + ui;
@@ -478,9 +487,9 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
         }
         // chunk-local solution: u <- gamma (d u + W (p m u)) - r
         lds[lane] = pos ? pi * u : 0.f;
-        __syncthreads();
+        lds_barrier();
         const float y = fmaf(di, u, lds_dot<MP>(lds, un, wrow));
-        __syncthreads();
+        lds_barrier();
         if (run) {
             u = fmaf(ugam, y, -r);
             zprev = zcur;
@@ -503,22 +512,31 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
 }
 
 // ---------------------------------------------------------------------------------------
-// carries across chunks (one block of MP lanes per sequence)
+// carries across chunks
 //   forward: carry_in[c] = y_end(c-1),  y_end(c) = P_c y_end(c-1) + v_c
 //   reverse: carry_in[c] = lam_{s1(c)}, lam_{s0(c)} = P_c^T lam_{s1(c)} + v_c
+// In processing order k (k = c forward, c = ncs - 1 - k reverse) both read
+//   carry_in[c(k)] = cur_k,  cur_{k+1} = A_k cur_k + v_{c(k)},  A_k = P_c or P_c^T.
+// Long chunk sequences use two levels: groups of G consecutive k are composed into one map
+// (Q_j, u_j) (k_carry_group, all groups in parallel), the group carries are walked serially
+// (k_carry over the groups), and every group re-walks its chunks from its carry (k_carry with
+// a start vector).  Serial depth G + ncs / G + G instead of ncs.
 // ---------------------------------------------------------------------------------------
 template <int MP, bool REV>
 __global__ __launch_bounds__(MP) void k_carry(const float *__restrict__ P, const float *__restrict__ v,
                                               float *__restrict__ carry_in, const int *__restrict__ active,
-                                              uint32_t *__restrict__ norm_bits, int ncs) {
+                                              uint32_t *__restrict__ norm_bits, int B, int ncs, int G,
+                                              const float *__restrict__ start) {
     __shared__ __align__(16) float cs[MP];
-    const int b = blockIdx.x, i = threadIdx.x;
-    if (norm_bits && i == 0) {   // [0, B): max|Delta|, [B, 2B): max|z| of the next fix-up
+    const int ngroups = (ncs + G - 1) / G;
+    const int b = blockIdx.x / ngroups, j = blockIdx.x % ngroups, i = threadIdx.x;
+    if (norm_bits && j == 0 && i == 0) {   // [0, B): max|Delta|, [B, 2B): max|z| of the next fix-up
         norm_bits[b] = 0u;
-        norm_bits[gridDim.x + b] = 0u;
+        norm_bits[B + b] = 0u;
     }
     if (active && !active[b]) return;
-    float cur = 0.f;
+    const int k0 = j * G, k1 = min(k0 + G, ncs);
+    float cur = start ? start[((size_t)b * ngroups + j) * MP + i] : 0.f;
     float pr[MP], pn[MP];
     auto load = [&](int step, float *dst) {
         const int cc = REV ? ncs - 1 - step : step;
@@ -535,26 +553,97 @@ __global__ __launch_bounds__(MP) void k_carry(const float *__restrict__ P, const
             for (int k = 0; k < MP; ++k) dst[k] = Pc[k * MP + i];
         }
     };
-    load(0, pr);
-    for (int step = 0; step < ncs; ++step) {
+    load(k0, pr);
+    for (int step = k0; step < k1; ++step) {
         const int cc = REV ? ncs - 1 - step : step;
         const size_t id = (size_t)b * ncs + cc;
-        if (step + 1 < ncs) load(step + 1, pn);
+        if (step + 1 < k1) load(step + 1, pn);
         const float vv = v[id * MP + i];
         carry_in[id * MP + i] = cur;
         cs[i] = cur;
-        __syncthreads();
+        lds_barrier();
         float a0 = vv, a1 = 0.f;
 #pragma unroll
         for (int k = 0; k < MP; k += 2) {
             a0 = fmaf(pr[k], cs[k], a0);
             a1 = fmaf(pr[k + 1], cs[k + 1], a1);
         }
-        __syncthreads();
+        lds_barrier();
         cur = a0 + a1;
 #pragma unroll
         for (int k = 0; k < MP; ++k) pr[k] = pn[k];
     }
+}
+
+// group maps in processing order: Q_j = A_{k1-1} ... A_{k0}, u_j = the group's walk from 0
+template <int MP, bool REV>
+__global__ __launch_bounds__(256) void k_carry_group(const float *__restrict__ P, const float *__restrict__ v,
+                                                     float *__restrict__ gq, float *__restrict__ gu,
+                                                     const int *__restrict__ active, int ncs, int G) {
+    constexpr int E = (MP * MP + 255) / 256;
+    __shared__ float Q[MP][MP + 1], Am[MP][MP + 1], u[MP], vv[MP];
+    const int ngroups = (ncs + G - 1) / G;
+    const int b = blockIdx.x / ngroups, j = blockIdx.x % ngroups, tid = threadIdx.x;
+    if (active && !active[b]) return;
+    for (int e = tid; e < MP * MP; e += 256) Q[e / MP][e % MP] = (e / MP == e % MP) ? 1.f : 0.f;
+    if (tid < MP) u[tid] = 0.f;
+    const int k0 = j * G, k1 = min(k0 + G, ncs);
+    // the next step's matrix and vector are loaded while this step is composed
+    float pn[E], vn = 0.f;
+    auto fetch = [&](int step) {
+        const int cc = REV ? ncs - 1 - step : step;
+        const float *Pc = P + ((size_t)b * ncs + cc) * MP * MP;
+#pragma unroll
+        for (int t = 0; t < E; ++t) {
+            const int e = tid + 256 * t;
+            pn[t] = (step < k1 && e < MP * MP) ? Pc[e] : 0.f;
+        }
+        vn = (step < k1 && tid < MP) ? v[((size_t)b * ncs + cc) * MP + tid] : 0.f;
+    };
+    fetch(k0);
+    for (int step = k0; step < k1; ++step) {
+#pragma unroll
+        for (int t = 0; t < E; ++t) {
+            const int e = tid + 256 * t;
+            if (e < MP * MP) {
+                const int r = e / MP, col = e % MP;
+                if (REV) Am[col][r] = pn[t];
+                else Am[r][col] = pn[t];
+            }
+        }
+        if (tid < MP) vv[tid] = vn;
+        fetch(step + 1);
+        lds_barrier();
+        float qn[E];
+#pragma unroll
+        for (int t = 0; t < E; ++t) {
+            const int e = tid + 256 * t;
+            float acc = 0.f;
+            if (e < MP * MP) {
+                const int r = e / MP, col = e % MP;
+#pragma unroll
+                for (int k = 0; k < MP; ++k) acc = fmaf(Am[r][k], Q[k][col], acc);
+            }
+            qn[t] = acc;
+        }
+        float un = 0.f;
+        if (tid < MP) {
+            un = vv[tid];
+#pragma unroll
+            for (int k = 0; k < MP; ++k) un = fmaf(Am[tid][k], u[k], un);
+        }
+        lds_barrier();
+#pragma unroll
+        for (int t = 0; t < E; ++t) {
+            const int e = tid + 256 * t;
+            if (e < MP * MP) Q[e / MP][e % MP] = qn[t];
+        }
+        if (tid < MP) u[tid] = un;
+        lds_barrier();
+    }
+    float *q = gq + ((size_t)b * ngroups + j) * MP * MP;
+    for (int e = tid; e < MP * MP; e += 256) q[e] = Q[e / MP][e % MP];
+    if (tid < MP) gu[((size_t)b * ngroups + j) * MP + tid] = u[tid];
 }
 
 // ---------------------------------------------------------------------------------------
@@ -565,7 +654,7 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict_
                                                         float alpha, int N, const uint32_t *__restrict__ masks,
                                                         const float *__restrict__ r, const float *__restrict__ carry_in,
                                                         const float *zin, float *zout,
-                                                        uint32_t *__restrict__ norm_bits, const int *__restrict__ active,
+                                                        uint32_t *__restrict__ chain_bits, const int *__restrict__ active,
                                                         const float *__restrict__ gamma, int B, int T, int M, int C,
                                                         int ncs) {
     using G = Geo<MP>;
@@ -584,19 +673,39 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict_
     float D = (ok && i < M) ? carry_in[(size_t)id * MP + i] : 0.f;
     uint32_t emax = 0u, zmax = 0u;
     const int maxlen = __builtin_amdgcn_readfirstlane(C);
+    // the loads of a step are issued PD steps ahead
+    auto fetch = [&](int t, float &rv, float &zv, uint32_t &mw) {
+        const bool run = t < len && i < M;
+        const size_t step = (size_t)b * T + s0 + t;
+        rv = run ? r[step * M + i] : 0.f;
+        zv = run ? zin[step * M + i] : 0.f;
+        mw = run ? masks[step * G::MW + (i >> 5)] : 0u;
+    };
+    constexpr int PD = 2;
+    float rq[PD], zq[PD];
+    uint32_t mq[PD];
+#pragma unroll
+    for (int q = 0; q < PD; ++q) fetch(q, rq[q], zq[q], mq[q]);
     for (int t = 0; t < maxlen; ++t) {
         const bool run = t < len && i < M;
         const size_t step = (size_t)b * T + s0 + t;
-        lds[lane] = (run && mask_bit(masks, step, G::MW, i)) ? D : 0.f;
-        __syncthreads();
+        const float rc = rq[0], zc = zq[0];
+        const uint32_t mc = mq[0];
+#pragma unroll
+        for (int q = 0; q + 1 < PD; ++q) {
+            rq[q] = rq[q + 1];
+            zq[q] = zq[q + 1];
+            mq[q] = mq[q + 1];
+        }
+        fetch(t + PD, rq[PD - 1], zq[PD - 1], mq[PD - 1]);
+        lds[lane] = (run && ((mc >> (i & 31)) & 1u)) ? D : 0.f;
+        lds_barrier();
         const float y = fmaf(d, D, lds_dot<MP>(lds, n, wrow));
-        __syncthreads();
+        lds_barrier();
         if (run) {
-            D = fmaf(gm, y, -r[step * M + i]);
-            const size_t e = step * M + i;
-            const float zo = zin[e];
-            zout[e] = zo + D;
-            const uint32_t ab = abs_bits(D), zb = abs_bits(zo);
+            D = fmaf(gm, y, -rc);
+            zout[step * M + i] = zc + D;
+            const uint32_t ab = abs_bits(D), zb = abs_bits(zc);
             emax = emax > ab ? emax : ab;
             zmax = zmax > zb ? zmax : zb;
         }
@@ -609,10 +718,49 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict_
         emax = emax > o ? emax : o;
         zmax = zmax > oz ? zmax : oz;
     }
-    if (ok && i == 0) {
-        atomicMax(norm_bits + b, emax);
-        atomicMax(norm_bits + B + b, zmax);
+    if (ok && i == 0) {   // per-chain maxima, reduced per sequence by k_seq_max
+        chain_bits[id] = emax;
+        chain_bits[(size_t)B * ncs + id] = zmax;
     }
+}
+
+// per-sequence max over its chains of the bits the forward fix-ups left:
+// norm_bits[b] = max |Delta|, norm_bits[B + b] = max |z| (unsigned max of |x| bits, NaN-propagating)
+__global__ __launch_bounds__(256) void k_seq_max(const uint32_t *__restrict__ chain_bits, const int *__restrict__ active,
+                                                 uint32_t *__restrict__ norm_bits, int B, int ncs) {
+    __shared__ uint32_t red[2][4];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    if (active && !active[b]) return;
+    uint32_t e = 0u, zm = 0u;
+    for (int c = tid; c < ncs; c += 256) {
+        const uint32_t a = chain_bits[(size_t)b * ncs + c], z = chain_bits[(size_t)B * ncs + (size_t)b * ncs + c];
+        e = e > a ? e : a;
+        zm = zm > z ? zm : z;
+    }
+    e = wave_max_u32(e);
+    zm = wave_max_u32(zm);
+    if ((tid & 63) == 0) {
+        red[0][tid >> 6] = e;
+        red[1][tid >> 6] = zm;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t a = red[0][0], z = red[1][0];
+        for (int w = 1; w < 4; ++w) {
+            a = a > red[0][w] ? a : red[0][w];
+            z = z > red[1][w] ? z : red[1][w];
+        }
+        norm_bits[b] = a;
+        norm_bits[B + b] = z;
+    }
+}
+
+int launch_seq_max(const uint32_t *chain_bits, const int *active, uint32_t *norm_bits, int B, int ncs,
+                   hipStream_t st) {
+    KTimer kt("k_seq_max", st);
+    hipLaunchKernelGGL(k_seq_max, dim3(B), dim3(256), 0, st, chain_bits, active, norm_bits, B, ncs);
+    DEER_LAUNCH_CHECK("k_seq_max");
+    return DEER_OK;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -645,33 +793,53 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn(const float *__restrict_
     float lam = (ok && i < M) ? carry_in[(size_t)id * MP + i] : 0.f;
     float dA = 0.f, dh = 0.f;
     const int maxlen = __builtin_amdgcn_readfirstlane(C);
+    // per-step inputs (mask of step k + 1, cotangent g_k, forced state z~_{k-1}), PD steps ahead
+    auto fetch = [&](int t, float &mv, float &gv, float &zv) {
+        const int k = s1 - 1 - t;
+        const bool run = k >= s0 && i < M;
+        mv = 0.f;
+        gv = 0.f;
+        zv = 0.f;
+        if (run) {
+            const size_t step = (size_t)b * T + k;
+            if (k + 1 < T) mv = (float)mask_bit(masks, step + 1, G::MW, i);
+            if (gin) gv = gin[step * M + i];
+            else if (i < N) gv = seed_scale * (z[step * M + i] - x[((size_t)b * (T + 1) + k + 1) * N + i]);
+            zv = forced_state(x, z0, z, b, k, i, T, M, N, alpha);
+        }
+    };
+    constexpr int PD = 1;
+    float mq[PD], gq[PD], zq[PD];
+#pragma unroll
+    for (int q = 0; q < PD; ++q) fetch(q, mq[q], gq[q], zq[q]);
     for (int t = 0; t < maxlen; ++t) {
         const int k = s1 - 1 - t;
         const bool run = k >= s0 && i < M;
+        const float mc = mq[0], gk = gq[0], zc = zq[0];
+#pragma unroll
+        for (int q = 0; q + 1 < PD; ++q) {
+            mq[q] = mq[q + 1];
+            gq[q] = gq[q + 1];
+            zq[q] = zq[q + 1];
+        }
+        fetch(t + PD, mq[PD - 1], gq[PD - 1], zq[PD - 1]);
         lds[lane] = lam;
-        __syncthreads();
+        lds_barrier();
         const float wt = lds_dot<MP>(lds, n, wcol);
-        __syncthreads();
+        lds_barrier();
         float zt = 0.f;
         if (run) {
             const size_t step = (size_t)b * T + k;
-            float y = 0.f;
-            if (k + 1 < T) {
-                const float m = (float)mask_bit(masks, step + 1, G::MW, i);
-                y = pi * fmaf(Ai, lam, m * wt);
-            }
-            float gk;
-            if (gin) gk = gin[step * M + i];
-            else gk = i < N ? seed_scale * (z[step * M + i] - x[((size_t)b * (T + 1) + k + 1) * N + i]) : 0.f;
+            const float y = (k + 1 < T) ? pi * fmaf(Ai, lam, mc * wt) : 0.f;
             lam = y + gk;
             if (lam_out) lam_out[step * M + i] = lam;
-            zt = forced_state(x, z0, z, b, k, i, T, M, N, alpha);
+            zt = zc;
             dA = fmaf(lam, zt, dA);
             dh += lam;
         }
         const float lr = run ? lam : 0.f;
         lds[lane] = (run && zt > 0.f) ? zt : 0.f;
-        __syncthreads();
+        lds_barrier();
         const float4 *l4 = reinterpret_cast<const float4 *>(lds + n * MP);
 #pragma unroll
         for (int q = 0; q < MP / 4; ++q) {
@@ -681,7 +849,7 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn(const float *__restrict_
             dW[4 * q + 2] = fmaf(lr, v.z, dW[4 * q + 2]);
             dW[4 * q + 3] = fmaf(lr, v.w, dW[4 * q + 3]);
         }
-        __syncthreads();
+        lds_barrier();
     }
     if (ok) {
         float *gp = gpart + ((size_t)id * MP + i) * (MP + 2);
@@ -796,35 +964,77 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, float *r, ui
     return DEER_OK;
 }
 
+// two-level carry for chunk sequences at least this long (MP <= 32)
+static int carry_group_size(int MP, int ncs) {
+    if (MP > 32 || ncs < 96) return 0;
+    int G = 8;
+    while (2 * G * G < ncs) G <<= 1;   // a group step costs about twice a walk step
+    return G;
+}
+
+size_t carry_ws_floats(int MP, int B, int ncs) {
+    const int G = carry_group_size(MP, ncs);
+    if (!G) return 0;
+    const size_t ng = (size_t)(ncs + G - 1) / G;
+    return (size_t)B * ng * ((size_t)MP * MP + 2 * MP);
+}
+
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
-                 uint32_t *norm_bits, int B, int ncs, hipStream_t st) {
+                 uint32_t *norm_bits, int B, int ncs, float *gws, hipStream_t st) {
     KTimer kt("k_carry", st);
-#define CA(MPV, R) \
-    hipLaunchKernelGGL((k_carry<MPV, R>), dim3(B), dim3(MPV), 0, st, P, v, carry_in, active, norm_bits, ncs)
-    if (!rev) {
-        if (MP == 16) CA(16, false); else if (MP == 32) CA(32, false); else CA(64, false);
+    const int G = gws ? carry_group_size(MP, ncs) : 0;
+#define CA(MPV, R, PP, VV, CI, NB, NC, GG, ST, GRID) \
+    hipLaunchKernelGGL((k_carry<MPV, R>), dim3(GRID), dim3(MPV), 0, st, PP, VV, CI, active, NB, B, NC, GG, ST)
+#define CG(MPV, R, GRID) \
+    hipLaunchKernelGGL((k_carry_group<MPV, R>), dim3(GRID), dim3(256), 0, st, P, v, gq, gu, active, ncs, G)
+    if (!G) {
+        if (!rev) {
+            if (MP == 16) CA(16, false, P, v, carry_in, norm_bits, ncs, ncs, nullptr, B);
+            else if (MP == 32) CA(32, false, P, v, carry_in, norm_bits, ncs, ncs, nullptr, B);
+            else CA(64, false, P, v, carry_in, norm_bits, ncs, ncs, nullptr, B);
+        } else {
+            if (MP == 16) CA(16, true, P, v, carry_in, norm_bits, ncs, ncs, nullptr, B);
+            else if (MP == 32) CA(32, true, P, v, carry_in, norm_bits, ncs, ncs, nullptr, B);
+            else CA(64, true, P, v, carry_in, norm_bits, ncs, ncs, nullptr, B);
+        }
     } else {
-        if (MP == 16) CA(16, true); else if (MP == 32) CA(32, true); else CA(64, true);
+        const int ng = (ncs + G - 1) / G;
+        float *gq = gws;
+        float *gu = gq + (size_t)B * ng * MP * MP;
+        float *gc = gu + (size_t)B * ng * MP;
+        const int grid = B * ng;
+        if (MP == 16) {
+            if (rev) CG(16, true, grid); else CG(16, false, grid);
+            CA(16, false, gq, gu, gc, nullptr, ng, ng, nullptr, B);
+            if (rev) CA(16, true, P, v, carry_in, norm_bits, ncs, G, gc, grid);
+            else CA(16, false, P, v, carry_in, norm_bits, ncs, G, gc, grid);
+        } else {
+            if (rev) CG(32, true, grid); else CG(32, false, grid);
+            CA(32, false, gq, gu, gc, nullptr, ng, ng, nullptr, B);
+            if (rev) CA(32, true, P, v, carry_in, norm_bits, ncs, G, gc, grid);
+            else CA(32, false, P, v, carry_in, norm_bits, ncs, G, gc, grid);
+        }
     }
+#undef CG
 #undef CA
     DEER_LAUNCH_CHECK("k_carry");
     return DEER_OK;
 }
 
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
-                           const float *zin, float *zout, uint32_t *norm_bits, const int *active, const float *gamma,
-                           int C, int ncs, hipStream_t st) {
+                           const float *zin, float *zout, uint32_t *chain_bits, uint32_t *norm_bits,
+                           const int *active, const float *gamma, int C, int ncs, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt("k_fixup_fwd_plrnn", st);
 #define FX(MPV)                                                                                                       \
     hipLaunchKernelGGL(k_fixup_fwd_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, carry_in, \
-                       zin, zout, norm_bits, active, gamma, a.B, a.T, a.M, C, ncs)
+                       zin, zout, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
     if (MP == 16) FX(16); else if (MP == 32) FX(32); else FX(64);
 #undef FX
     DEER_LAUNCH_CHECK("k_fixup_fwd_plrnn");
-    return DEER_OK;
+    return launch_seq_max(chain_bits, active, norm_bits, a.B, ncs, st);
 }
 
 int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *g, float seed_scale, const float *z,

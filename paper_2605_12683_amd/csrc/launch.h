@@ -31,10 +31,13 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
 int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, float *r, uint32_t *masks, float *P, float *v,
                                 const int *active, const float *gamma, int C, int ncs, hipStream_t st);
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
-                 uint32_t *norm_bits, int B, int ncs, hipStream_t st);
+                 uint32_t *norm_bits, int B, int ncs, float *gws, hipStream_t st);
+size_t carry_ws_floats(int MP, int B, int ncs);
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
-                           const float *zin, float *zout, uint32_t *norm_bits, const int *active, const float *gamma,
-                           int C, int ncs, hipStream_t st);
+                           const float *zin, float *zout, uint32_t *chain_bits, uint32_t *norm_bits,
+                           const int *active, const float *gamma, int C, int ncs, hipStream_t st);
+int launch_seq_max(const uint32_t *chain_bits, const int *active, uint32_t *norm_bits, int B, int ncs,
+                   hipStream_t st);
 int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *g, float seed_scale, const float *z,
                            const float *carry_in, float *lam, float *gpart, int C, int ncs, hipStream_t st);
 int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *dA, float *dW, float *dh,
@@ -45,8 +48,8 @@ size_t reduce_gpart_ws_bytes(int MP);
 int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
                                float *P, float *v, const int *active, int C, int ncs, hipStream_t st);
 int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
-                       const float *carry_in, const float *zin, float *out, uint32_t *norm_bits, const int *active,
-                       int C, int ncs,
+                       const float *carry_in, const float *zin, float *out, uint32_t *chain_bits, uint32_t *norm_bits,
+                       const int *active, int C, int ncs,
                        hipStream_t st);
 
 // shallow PLRNN

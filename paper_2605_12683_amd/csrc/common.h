@@ -74,6 +74,16 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 
 // forced input of step s (array index) for latent i:
 //   s == 0: z0 (or [x_0; 0] when z0 is null);  s >= 1: fl(fl(p*z_{s-1}) + fl(a*zbar_s))
+// The two iterate buffers of the safeguarded Newton loop: sequence b's current iterate is in
+// zalt when zsel[b] is set, else in z, and an update is written to the other buffer.  With
+// zsel null and zalt == z the update is applied in place.
+__device__ __forceinline__ const float *cur_iter(const float *z, const float *zalt, const int *zsel, int b) {
+    return (zsel && zsel[b]) ? zalt : z;
+}
+__device__ __forceinline__ float *next_iter(float *z, float *zalt, const int *zsel, int b) {
+    return (zsel && zsel[b]) ? z : zalt;
+}
+
 // Workgroup barrier that orders LDS only: unlike __syncthreads it does not wait for
 // outstanding global loads, so loads issued ahead (prefetch) stay in flight across it.  For
 // kernels whose threads exchange data through LDS alone.

@@ -159,12 +159,13 @@ static int choose_chunk(int B, int T, int MP) {
     return (int)C;
 }
 
-// Per-sequence control block of the Newton loop: active flags [B] followed by the damping
-// factors gamma [B] (one host-to-device copy updates both), and 2B words of max bits
-// (max|Delta| and max|z| of the last fix-up).
+// Per-sequence control block of the Newton loop (device, 7B words, one device-to-host copy
+// reads all of it): act | gamma | sel | om | it | norm | status (see NewtonDev), then 2B
+// words of max bits for the fixed-iteration mode, the per-chain maxima of a pass, and the
+// second iterate buffer.
 struct NewtonCtl {
-    int *active;
-    float *gamma;
+    NewtonDev nd;
+    uint32_t *blk;          // start of the 7B-word block
     uint32_t *norm_bits;
     uint32_t *chain_bits;   // per-chain maxima [2][B * ncs] before the per-sequence reduction
     float *zalt;            // second iterate buffer [B,T,M]
@@ -172,9 +173,17 @@ struct NewtonCtl {
 
 static NewtonCtl carve_ctl(Carver &c, int B, size_t seq_elems, size_t nchains) {
     NewtonCtl n{};
-    uint32_t *blk = c.take<uint32_t>(2 * (size_t)B);
-    n.active = (int *)blk;
-    n.gamma = blk ? (float *)(blk + B) : nullptr;
+    uint32_t *blk = c.take<uint32_t>(7 * (size_t)B);
+    n.blk = blk;
+    if (blk) {
+        n.nd.act = (int *)blk;
+        n.nd.gamma = (float *)(blk + B);
+        n.nd.sel = (int *)(blk + 2 * B);
+        n.nd.om = (float *)(blk + 3 * B);
+        n.nd.it = (int *)(blk + 4 * B);
+        n.nd.norm = (float *)(blk + 5 * B);
+        n.nd.status = (int *)(blk + 6 * B);
+    }
     n.norm_bits = c.take<uint32_t>(2 * (size_t)B);
     n.chain_bits = c.take<uint32_t>(2 * nchains);
     n.zalt = c.take<float>((size_t)B * seq_elems);
@@ -311,35 +320,37 @@ static size_t diag_bytes(int B, int T, int M, int K, int op) {
     return op == DEER_OP_ADJOINT ? diag_adjoint_ws_bytes(B, T, M, K) : diag_scan_ws_bytes(B, T, M);
 }
 
-// Host-side Newton loop shared by the PLRNN kinds.  `update(active, gamma, zin, zout)` queues
-// one Newton update of the sequences whose device flag is set (all, when active is null),
-// linearised with the per-sequence factor gamma (gamma J~; null: 1), reading the iterate from
-// zin and writing zin + Delta to zout (which may alias zin), and leaves per-sequence
-// max|Delta| and max|zin| bits in norm_bits[0, B) and [B, 2B).
+// Newton loop shared by the PLRNN kinds.  `update(act, gamma, zsel, z, zalt)` queues one
+// Newton update of the sequences whose device flag is set (all, when act is null),
+// linearised with the per-sequence factor gamma (gamma J~; null: 1), reading each sequence's
+// iterate from the buffer zsel selects and writing iterate + Delta to the other one (zsel
+// null and zalt == z: in place), and leaves per-chain max|Delta| and max|z| bits in
+// ctl.chain_bits.
 //
-// With a convergence test (fixed_iters == 0) every update is checked before it is kept: an
-// update that is not finite, or whose max|Delta| exceeds step_bound (1 + max|z|), is
-// rejected and the sequence retried with gamma < 1; gamma returns to 1 over accepted
-// updates.  gamma = 1 is the exact Newton step, gamma = 0 the fixed-point (Picard) step
-// z_t <- F(z~_{t-1}); every gamma keeps the fixed point, and the prefix property (an update
-// makes at least one more leading step exact) holds for every gamma.  Iterates alternate
-// between z and ctl.zalt, so a rejection costs a copy of the rejected sequences only.
+// With a convergence test (fixed_iters == 0) the test and the update safeguard run on the
+// device after every pass (k_seq_ctl): an update that is not finite, or whose max|Delta|
+// exceeds step_bound (1 + max|z|), is not kept and the sequence is retried with gamma < 1;
+// gamma returns to 1 over accepted updates.  gamma = 1 is the exact Newton step, gamma = 0
+// the fixed-point step z_t <- F(z~_{t-1}); every gamma keeps the fixed point and the prefix
+// property.  The host queues passes in batches and reads the active flags once per batch;
+// a sequence frozen inside a batch makes the rest of the batch's kernels skip it.
 constexpr float kDefaultStepBound = 1e3f;
-constexpr float kDampFirst = 1.f / 64, kDampGrow = 4.f, kDampShrink = 4.f, kDampFloor = 1e-4f;
+constexpr NewtonDamp kDamp = {1.f / 64, 4.f, 4.f, 1e-4f};
+constexpr int kFirstBatch = 4, kBatch = 2;
 
 template <class Update>
-static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, const NewtonCtl &ctl, float *z,
+static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int ncs, const NewtonCtl &ctl, float *z,
                        Update update, std::vector<int> &it, std::vector<float> &norm, bool &nonfinite,
                        std::vector<int> &act, hipStream_t st) {
     const int fixed = o->fixed_iters > 0 ? o->fixed_iters : 0;
     const int max_iter = o->max_iter > 0 ? o->max_iter : 500;
     const float bound = o->step_bound == 0.f ? kDefaultStepBound : o->step_bound;
-    const size_t seq_bytes = seq_elems * sizeof(float);
     int rc;
-    std::vector<uint32_t> nb(2 * (size_t)B, 0);
     if (fixed) {
         for (int k = 0; k < fixed; ++k)
-            if ((rc = update(nullptr, nullptr, z, z))) return rc;
+            if ((rc = update(nullptr, nullptr, nullptr, z, z))) return rc;
+        if ((rc = launch_seq_max(ctl.chain_bits, nullptr, ctl.norm_bits, B, ncs, st))) return rc;
+        std::vector<uint32_t> nb(B, 0);
         DEER_HIP(hipMemcpyAsync(nb.data(), ctl.norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
         DEER_HIP(hipStreamSynchronize(st));
         for (int b = 0; b < B; ++b) {
@@ -349,87 +360,36 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, const 
         }
         return DEER_OK;
     }
-    // host mirror of the control block: act [B] | gamma [B]
-    std::vector<uint32_t> hctl(2 * (size_t)B);
-    std::vector<float> om(B, 0.f);   // 1 - gamma
-    auto push_ctl = [&]() -> int {
-        for (int b = 0; b < B; ++b) {
-            hctl[b] = (uint32_t)act[b];
-            const float gm = 1.f - om[b];
-            memcpy(&hctl[B + b], &gm, 4);
+    const NewtonDev &nd = ctl.nd;
+    if ((rc = launch_ctl_init(nd, B, st))) return rc;
+    int passes = 0, batch = kFirstBatch;
+    while (passes < max_iter) {
+        const int n = batch < max_iter - passes ? batch : max_iter - passes;
+        for (int k = 0; k < n; ++k) {
+            if ((rc = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt))) return rc;
+            if ((rc = launch_seq_ctl(ctl.chain_bits, nd, B, ncs, o->tol, bound, kDamp, st))) return rc;
         }
-        DEER_HIP(hipMemcpyAsync(ctl.active, hctl.data(), 2 * B * sizeof(uint32_t), hipMemcpyHostToDevice, st));
+        passes += n;
+        DEER_HIP(hipMemcpyAsync(act.data(), nd.act, B * sizeof(int), hipMemcpyDeviceToHost, st));
         DEER_HIP(hipStreamSynchronize(st));
-        return DEER_OK;
-    };
-    if ((rc = push_ctl())) return rc;
-    float *buf[2] = {z, ctl.zalt};
-    int cur = 0;
-    std::vector<int> holder(B, 0);   // buffer that holds each sequence's iterate
-    std::vector<int> acc, rej;
-    for (int k = 0;; ++k) {
         bool any = false;
         for (int b = 0; b < B; ++b) any |= act[b] != 0;
-        if (!any || k == max_iter) break;
-        if ((rc = update(ctl.active, ctl.gamma, buf[cur], buf[1 - cur]))) return rc;
-        DEER_HIP(hipMemcpyAsync(nb.data(), ctl.norm_bits, 2 * B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
-        DEER_HIP(hipStreamSynchronize(st));
-        bool changed = false;
-        acc.clear();
-        rej.clear();
-        for (int b = 0; b < B; ++b) {
-            if (!act[b]) continue;
-            float e, zn;
-            memcpy(&e, &nb[b], 4);
-            memcpy(&zn, &nb[B + b], 4);
-            const bool fin = isfinite(e);
-            const bool keep = fin && (bound < 0.f || om[b] >= 1.f || e <= bound * (1.f + zn));
-            if (keep) {
-                acc.push_back(b);
-                it[b] += 1;
-                norm[b] = e;
-                if (om[b] > 0.f) {
-                    om[b] = om[b] / kDampShrink < kDampFloor ? 0.f : om[b] / kDampShrink;
-                    changed = true;
-                }
-                if (e < o->tol) {
-                    act[b] = 0;
-                    changed = true;
-                }
-            } else if (om[b] >= 1.f) {
-                // the fixed-point step itself overflows: the trajectory is not finite
-                rej.push_back(b);
-                norm[b] = e;
-                nonfinite = true;
-                act[b] = 0;
-                changed = true;
-            } else {
-                rej.push_back(b);
-                om[b] = om[b] == 0.f ? kDampFirst : (om[b] * kDampGrow > 1.f ? 1.f : om[b] * kDampGrow);
-                changed = true;
-            }
-        }
-        // keep every sequence's iterate in one buffer: copy the smaller set across
-        if (!acc.empty()) {
-            if (acc.size() >= rej.size()) {
-                for (int b : rej)
-                    DEER_HIP(hipMemcpyAsync(buf[1 - cur] + b * seq_elems, buf[cur] + b * seq_elems, seq_bytes,
-                                            hipMemcpyDeviceToDevice, st));
-                cur = 1 - cur;
-            } else {
-                for (int b : acc)
-                    DEER_HIP(hipMemcpyAsync(buf[cur] + b * seq_elems, buf[1 - cur] + b * seq_elems, seq_bytes,
-                                            hipMemcpyDeviceToDevice, st));
-            }
-        }
-        for (int b : acc) holder[b] = cur;
-        for (int b : rej) holder[b] = cur;
-        if (changed && (rc = push_ctl())) return rc;
+        if (!any) break;
+        batch = kBatch;
     }
-    for (int b = 0; b < B; ++b)
-        if (holder[b] == 1)
+    std::vector<uint32_t> h(7 * (size_t)B);
+    DEER_HIP(hipMemcpyAsync(h.data(), ctl.blk, h.size() * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+    DEER_HIP(hipStreamSynchronize(st));
+    const size_t seq_bytes = seq_elems * sizeof(float);
+    for (int b = 0; b < B; ++b) {
+        act[b] = (int)h[b];
+        it[b] = (int)h[4 * (size_t)B + b];
+        memcpy(&norm[b], &h[5 * (size_t)B + b], 4);
+        if (h[6 * (size_t)B + b] == 2u) nonfinite = true;
+        if (h[2 * (size_t)B + b])   // the iterate ended in the second buffer
             DEER_HIP(hipMemcpyAsync(z + b * seq_elems, ctl.zalt + b * seq_elems, seq_bytes, hipMemcpyDeviceToDevice,
                                     st));
+    }
     return DEER_OK;
 }
 
@@ -470,15 +430,15 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     std::vector<int> act(B, 1), it(B, 0);
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
-    uint32_t *nbits = w.ctl.norm_bits;
-    auto update = [&](const int *dact, const float *gam, const float *zin, float *zout) -> int {
+    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za) -> int {
         int r;
-        if ((r = launch_newton_product_plrnn(a, zin, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, st))) return r;
-        if ((r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, nbits, B, w.ncs, w.gws, st))) return r;
-        return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, zin, zout, w.ctl.chain_bits, nbits, dact, gam, w.C,
-                                      w.ncs, st);
+        if ((r = launch_newton_product_plrnn(a, zb, za, zsel, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, st)))
+            return r;
+        if ((r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, nullptr, B, w.ncs, w.gws, st))) return r;
+        return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, zb, za, zsel, w.ctl.chain_bits, dact, gam, w.C, w.ncs,
+                                      st);
     };
-    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
+    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ncs, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
         if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
     }
@@ -500,19 +460,18 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
     const DenseWs &d = w.d;
-    uint32_t *nbits = w.ctl.norm_bits;
-    auto update = [&](const int *dact, const float *gam, const float *zin, float *zout) -> int {
+    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za) -> int {
         int r;
-        if ((r = launch_resjac_shplrnn(a, zin, nullptr, w.r, w.masks, dact, st))) return r;
+        if ((r = launch_resjac_shplrnn(a, zb, za, zsel, nullptr, w.r, w.masks, dact, st))) return r;
         if ((r = launch_jacform_shplrnn(a, w.masks, w.J, dact, gam, st))) return r;
         if ((r = launch_chunk_product_dense(false, B, T, m->M, w.J, w.r, -1.f, d.P, d.v, dact, d.C, d.ncs, st))) return r;
-        if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nbits, B, d.ncs, d.gws, st))) return r;
-        return launch_fixup_dense(0, B, T, m->M, w.J, w.r, -1.f, d.carry, zin, zout, w.ctl.chain_bits, nbits, dact,
-                                  d.C, d.ncs, st);
+        if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nullptr, B, d.ncs, d.gws, st))) return r;
+        return launch_fixup_dense(0, B, T, m->M, w.J, w.r, -1.f, d.carry, zb, za, zsel, w.ctl.chain_bits, dact, d.C,
+                                  d.ncs, st);
     };
-    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
+    if ((rc = newton_loop(o, B, (size_t)T * m->M, d.ncs, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
-        if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, masks, nullptr, st))) return rc;
+        if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
     }
     return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
 }
@@ -616,7 +575,7 @@ int plrnn_jacobian(const deer_model *m, const deer_forcing *f, int B, int T, con
     if (m->kind == DEER_SHPLRNN) {
         if ((rc = check_shallow_limits(m))) return rc;
         ShArgs a{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
-        if ((rc = launch_resjac_shplrnn(a, z, F, r, masks, nullptr, st))) return rc;
+        if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, F, r, masks, nullptr, st))) return rc;
         if (J) {
             if (!masks) { set_error("the shallow dense Jacobian output needs the masks output"); return DEER_ERR_INVALID_ARG; }
             if ((rc = launch_jacform_shplrnn(a, masks, J, nullptr, nullptr, st))) return rc;
@@ -707,7 +666,7 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
             gg = w.g;
         }
         float *lo = lam ? lam : w.lam;
-        if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, w.masks, nullptr, st))) return rc;
+        if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, nullptr, nullptr, w.masks, nullptr, st))) return rc;
         if ((rc = launch_jacform_shplrnn(a, w.masks, w.J, nullptr, nullptr, st))) return rc;
         if ((rc = launch_chunk_product_dense(true, B, T, m->M, w.J, gg, 1.f, d.P, d.v, nullptr, d.C, d.ncs, st))) return rc;
         if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, d.gws, st))) return rc;

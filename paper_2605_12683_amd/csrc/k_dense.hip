@@ -147,14 +147,15 @@ __global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restr
     }
 }
 
-// MODE 0: forward Newton fix-up (out = zin + Delta, zin may alias out; per-sequence max |Delta|
-//         and max |zin|)
+// MODE 0: forward Newton fix-up (next iterate = current + Delta, in place when the two buffers
+//         coincide; per-chain max |Delta| and max |z|)
 // MODE 1: forward bare scan (y written)
 // MODE 2: reverse (y_k = J_{k+1}^T y_{k+1} + b_k written)
 template <int MP, int MODE>
 __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J, const float *__restrict__ rhs,
                                                     float rhs_sign, const float *__restrict__ carry_in,
-                                                    const float *zin, float *out, uint32_t *__restrict__ chain_bits,
+                                                    float *zbuf, float *outbuf, const int *__restrict__ zsel,
+                                                    uint32_t *__restrict__ chain_bits,
                                                     const int *__restrict__ active, int B, int T, int M, int C,
                                                     int ncs) {
     using G = DGeo<MP>;
@@ -165,6 +166,9 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
     const int b = ok0 ? id / ncs : 0, cc = ok0 ? id % ncs : 0;
     const bool ok = ok0 && (!active || active[b]);
     const int s0 = cc * C, s1 = ok ? min(s0 + C, T) : s0;
+    // MODE 0: iterate buffers (zbuf, outbuf) selected per sequence; MODE 1, 2: y = outbuf
+    const float *zin = MODE == 0 ? cur_iter(zbuf, outbuf, zsel, b) : nullptr;
+    float *out = MODE == 0 ? next_iter(zbuf, outbuf, zsel, b) : outbuf;
     float y = (ok && i < M) ? carry_in[(size_t)id * MP + i] : 0.f;
     uint32_t emax = 0u, zmax = 0u;
     const int maxlen = __builtin_amdgcn_readfirstlane(C);
@@ -267,22 +271,21 @@ int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, co
 }
 
 int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
-                       const float *carry_in, const float *zin, float *out, uint32_t *chain_bits, uint32_t *norm_bits,
+                       const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
                        const int *active, int C, int ncs, hipStream_t st) {
     const int MP = padded_dim(M);
     const int nch = B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt(mode == 2 ? "k_fixup_dense_rev" : "k_fixup_dense_fwd", st);
 #define FXD(MPV, MO)                                                                                          \
-    hipLaunchKernelGGL((k_fixup_dense<MPV, MO>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, carry_in, zin, \
-                       out, chain_bits, active, B, T, M, C, ncs)
+    hipLaunchKernelGGL((k_fixup_dense<MPV, MO>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, carry_in, z, out, \
+                       zsel, chain_bits, active, B, T, M, C, ncs)
 #define FXD3(MO) \
     if (MP == 16) FXD(16, MO); else if (MP == 32) FXD(32, MO); else FXD(64, MO);
     if (mode == 0) { FXD3(0) } else if (mode == 1) { FXD3(1) } else { FXD3(2) }
 #undef FXD3
 #undef FXD
     DEER_LAUNCH_CHECK("k_fixup_dense");
-    if (mode == 0) return launch_seq_max(chain_bits, active, norm_bits, B, ncs, st);
     return DEER_OK;
 }
 

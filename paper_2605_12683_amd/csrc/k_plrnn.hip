@@ -314,9 +314,10 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn(
 template <int MP>
 __global__ __launch_bounds__(64) void k_newton_product_plrnn(
     const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
-    const float *__restrict__ x, const float *__restrict__ z0, const float *__restrict__ z,
-    float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout, float *__restrict__ vout,
-    const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C, int ncs) {
+    const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
+    const int *__restrict__ zsel, float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout,
+    float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
+    int ncs) {
     using G = Geo<MP>;
     constexpr int NCH = G::NCH, NI = G::NI, NS = G::NS, MW = G::MW;
     __shared__ __align__(16) float lds[64];
@@ -394,6 +395,7 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
 #pragma unroll
     for (int n = 0; n < NCH; ++n)
         if (n == un) ugam = gam[n];
+    const float *z = cur_iter(zbuf, zalt, zsel, ub);   // this lane's sequence's iterate
     // z_{s-1} for the first step of the chunk
     float zprev = 0.f;
     if (ulen > 0 && lat) {
@@ -653,7 +655,7 @@ template <int MP>
 __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict__ A, const float *__restrict__ W,
                                                         float alpha, int N, const uint32_t *__restrict__ masks,
                                                         const float *__restrict__ r, const float *__restrict__ carry_in,
-                                                        const float *zin, float *zout,
+                                                        float *zbuf, float *zalt, const int *__restrict__ zsel,
                                                         uint32_t *__restrict__ chain_bits, const int *__restrict__ active,
                                                         const float *__restrict__ gamma, int B, int T, int M, int C,
                                                         int ncs) {
@@ -666,6 +668,8 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict_
     const bool ok = ok0 && (!active || active[b]);
     const int s0 = cc * C, len = ok ? min(C, T - s0) : 0;
     const float gm = gamma ? gamma[b] : 1.f;
+    const float *zin = cur_iter(zbuf, zalt, zsel, b);
+    float *zout = next_iter(zbuf, zalt, zsel, b);
     float wrow[MP];
 #pragma unroll
     for (int k = 0; k < MP; ++k) wrow[k] = (i < M && k < M) ? W[i * M + k] * p_of(k, N, alpha) : 0.f;
@@ -760,6 +764,84 @@ int launch_seq_max(const uint32_t *chain_bits, const int *active, uint32_t *norm
     KTimer kt("k_seq_max", st);
     hipLaunchKernelGGL(k_seq_max, dim3(B), dim3(256), 0, st, chain_bits, active, norm_bits, B, ncs);
     DEER_LAUNCH_CHECK("k_seq_max");
+    return DEER_OK;
+}
+
+// Convergence test and update safeguard of one Newton pass, per sequence, on the device (so
+// that passes are queued without a host round trip).  From the maxima of the pass's chains:
+// accept the update (flip sel, count it, relax the damping, freeze the sequence once
+// max|Delta| < tol), or reject it (keep sel, raise the damping: 1 - gamma = first, then x grow
+// up to 1 = the fixed-point step); a non-finite fixed-point step ends the sequence.
+__global__ __launch_bounds__(256) void k_seq_ctl(const uint32_t *__restrict__ chain_bits, NewtonDev nd, int B,
+                                                 int ncs, float tol, float bound, NewtonDamp dp) {
+    __shared__ uint32_t red[2][4];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    if (!nd.act[b]) return;
+    uint32_t e = 0u, zm = 0u;
+    for (int c = tid; c < ncs; c += 256) {
+        const uint32_t a = chain_bits[(size_t)b * ncs + c], z = chain_bits[(size_t)B * ncs + (size_t)b * ncs + c];
+        e = e > a ? e : a;
+        zm = zm > z ? zm : z;
+    }
+    e = wave_max_u32(e);
+    zm = wave_max_u32(zm);
+    if ((tid & 63) == 0) {
+        red[0][tid >> 6] = e;
+        red[1][tid >> 6] = zm;
+    }
+    __syncthreads();
+    if (tid != 0) return;
+    for (int w = 1; w < 4; ++w) {
+        e = e > red[0][w] ? e : red[0][w];
+        zm = zm > red[1][w] ? zm : red[1][w];
+    }
+    const float ef = __uint_as_float(e), zf = __uint_as_float(zm);
+    const bool fin = e < 0x7f800000u;
+    float om = nd.om[b];
+    const bool keep = fin && (bound < 0.f || om >= 1.f || ef <= bound * (1.f + zf));
+    if (keep) {
+        nd.sel[b] ^= 1;
+        nd.it[b] += 1;
+        nd.norm[b] = ef;
+        if (om > 0.f) om = om / dp.shrink < dp.floor ? 0.f : om / dp.shrink;
+        if (ef < tol) {
+            nd.act[b] = 0;
+            nd.status[b] = 1;
+        }
+    } else if (om >= 1.f) {
+        nd.norm[b] = ef;
+        nd.act[b] = 0;
+        nd.status[b] = 2;
+    } else {
+        om = om == 0.f ? dp.first : fminf(1.f, om * dp.grow);
+    }
+    nd.om[b] = om;
+    nd.gamma[b] = 1.f - om;
+}
+
+int launch_seq_ctl(const uint32_t *chain_bits, const NewtonDev &nd, int B, int ncs, float tol, float bound,
+                   const NewtonDamp &dp, hipStream_t st) {
+    KTimer kt("k_seq_ctl", st);
+    hipLaunchKernelGGL(k_seq_ctl, dim3(B), dim3(256), 0, st, chain_bits, nd, B, ncs, tol, bound, dp);
+    DEER_LAUNCH_CHECK("k_seq_ctl");
+    return DEER_OK;
+}
+
+__global__ void k_ctl_init(NewtonDev nd, int B) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    nd.act[b] = 1;
+    nd.gamma[b] = 1.f;
+    nd.sel[b] = 0;
+    nd.om[b] = 0.f;
+    nd.it[b] = 0;
+    nd.norm[b] = __uint_as_float(0x7fc00000u);
+    nd.status[b] = 0;
+}
+
+int launch_ctl_init(const NewtonDev &nd, int B, hipStream_t st) {
+    hipLaunchKernelGGL(k_ctl_init, dim3((B + 255) / 256), dim3(256), 0, st, nd, B);
+    DEER_LAUNCH_CHECK("k_ctl_init");
     return DEER_OK;
 }
 
@@ -949,15 +1031,16 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
     return DEER_OK;
 }
 
-int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, float *r, uint32_t *masks, float *P, float *v,
-                                const int *active, const float *gamma, int C, int ncs, hipStream_t st) {
+int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
+                                uint32_t *masks, float *P, float *v, const int *active, const float *gamma, int C,
+                                int ncs, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt("k_newton_product_plrnn", st);
 #define NP(MPV)                                                                                                   \
     hipLaunchKernelGGL(k_newton_product_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, \
-                       a.z0, z, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs)
+                       a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs)
     if (MP == 16) NP(16); else if (MP == 32) NP(32); else NP(64);
 #undef NP
     DEER_LAUNCH_CHECK("k_newton_product_plrnn");
@@ -1022,19 +1105,19 @@ int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_
 }
 
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
-                           const float *zin, float *zout, uint32_t *chain_bits, uint32_t *norm_bits,
-                           const int *active, const float *gamma, int C, int ncs, hipStream_t st) {
+                           float *z, float *zalt, const int *zsel, uint32_t *chain_bits, const int *active,
+                           const float *gamma, int C, int ncs, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt("k_fixup_fwd_plrnn", st);
 #define FX(MPV)                                                                                                       \
     hipLaunchKernelGGL(k_fixup_fwd_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, carry_in, \
-                       zin, zout, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
+                       z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
     if (MP == 16) FX(16); else if (MP == 32) FX(32); else FX(64);
 #undef FX
     DEER_LAUNCH_CHECK("k_fixup_fwd_plrnn");
-    return launch_seq_max(chain_bits, active, norm_bits, a.B, ncs, st);
+    return DEER_OK;
 }
 
 int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *g, float seed_scale, const float *z,

@@ -24,9 +24,10 @@ __device__ __forceinline__ float p_at(int i, int N, float alpha) { return i < N 
 constexpr int SH_TT = 16;
 
 template <int MP>
-__global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const float *__restrict__ z,
-                                                        float *__restrict__ F_out, float *__restrict__ r_out,
-                                                        uint32_t *__restrict__ masks, const int *__restrict__ active) {
+__global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const float *zbuf, const float *zalt,
+                                                        const int *__restrict__ zsel, float *__restrict__ F_out,
+                                                        float *__restrict__ r_out, uint32_t *__restrict__ masks,
+                                                        const int *__restrict__ active) {
     extern __shared__ __align__(16) float smem[];
     const int M = a.M, L = a.L, T = a.T;
     float *zt = smem;                    // [SH_TT][MP], zero padded
@@ -50,7 +51,7 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
             float v = 0.f;
             if (row < total && i < M) {
                 const int b = (int)(row / T), s = (int)(row % T);
-                v = forced_state(a.x, a.z0, z, b, s, i, T, M, a.N, a.alpha);
+                v = forced_state(a.x, a.z0, cur_iter(zbuf, zalt, zsel, b), b, s, i, T, M, a.N, a.alpha);
             }
             zt[e] = v;
         }
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
             const float F = fmaf(a.A[i], ztv, acc0 + acc1) + (a.h1 ? a.h1[i] : 0.f);
             const size_t e2 = (size_t)row * M + i;
             if (F_out) F_out[e2] = F;
-            if (r_out) r_out[e2] = z[e2] - F;
+            if (r_out) r_out[e2] = cur_iter(zbuf, zalt, zsel, (int)(row / a.T))[e2] - F;
         }
     }
 }
@@ -354,16 +355,17 @@ static int sh_LP(int L) { return (L + 15) / 16 * 16; }
 
 size_t sh_jacform_lds(int M, int L) { return (size_t)2 * padded_dim(M) * sh_LP(L) * sizeof(float); }
 
-int launch_resjac_shplrnn(const ShArgs &a, const float *z, float *F, float *r, uint32_t *masks, const int *active,
-                          hipStream_t st) {
+int launch_resjac_shplrnn(const ShArgs &a, const float *z, const float *zalt, const int *zsel, float *F, float *r,
+                          uint32_t *masks, const int *active, hipStream_t st) {
     const long ntiles = ((long)a.B * a.T + SH_TT - 1) / SH_TT;
     const int grid = (int)(ntiles < 4096 ? ntiles : 4096);
     const size_t lds = sh_resjac_lds(a.M, a.L);
     KTimer kt("k_resjac_shplrnn", st);
     const int MP = padded_dim(a.M);
-    if (MP == 16) hipLaunchKernelGGL(k_resjac_shplrnn<16>, dim3(grid), dim3(256), lds, st, a, z, F, r, masks, active);
-    else if (MP == 32) hipLaunchKernelGGL(k_resjac_shplrnn<32>, dim3(grid), dim3(256), lds, st, a, z, F, r, masks, active);
-    else hipLaunchKernelGGL(k_resjac_shplrnn<64>, dim3(grid), dim3(256), lds, st, a, z, F, r, masks, active);
+#define RS(MPV) \
+    hipLaunchKernelGGL(k_resjac_shplrnn<MPV>, dim3(grid), dim3(256), lds, st, a, z, zalt, zsel, F, r, masks, active)
+    if (MP == 16) RS(16); else if (MP == 32) RS(32); else RS(64);
+#undef RS
     DEER_LAUNCH_CHECK("k_resjac_shplrnn");
     return DEER_OK;
 }

@@ -28,14 +28,31 @@ int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, 
 int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *masks, const float *rhs, const float *z,
                                float seed_scale, float *P, float *v, const int *active, int C, int ncs,
                                hipStream_t st);
-int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, float *r, uint32_t *masks, float *P, float *v,
-                                const int *active, const float *gamma, int C, int ncs, hipStream_t st);
+int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
+                                uint32_t *masks, float *P, float *v, const int *active, const float *gamma, int C,
+                                int ncs, hipStream_t st);
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
                  uint32_t *norm_bits, int B, int ncs, float *gws, hipStream_t st);
 size_t carry_ws_floats(int MP, int B, int ncs);
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
-                           const float *zin, float *zout, uint32_t *chain_bits, uint32_t *norm_bits,
-                           const int *active, const float *gamma, int C, int ncs, hipStream_t st);
+                           float *z, float *zalt, const int *zsel, uint32_t *chain_bits, const int *active,
+                           const float *gamma, int C, int ncs, hipStream_t st);
+// device-side Newton control (one entry per sequence)
+struct NewtonDev {
+    int *act;       // active flag (read by every kernel of a pass)
+    float *gamma;   // damping of the linearisation
+    int *sel;       // which iterate buffer holds the current iterate
+    float *om;      // 1 - gamma
+    int *it;        // accepted updates
+    float *norm;    // max |Delta| of the last accepted (or final) update
+    int *status;    // 0 running, 1 converged, 2 non-finite
+};
+struct NewtonDamp {
+    float first, grow, shrink, floor;
+};
+int launch_seq_ctl(const uint32_t *chain_bits, const NewtonDev &nd, int B, int ncs, float tol, float bound,
+                   const NewtonDamp &dp, hipStream_t st);
+int launch_ctl_init(const NewtonDev &nd, int B, hipStream_t st);
 int launch_seq_max(const uint32_t *chain_bits, const int *active, uint32_t *norm_bits, int B, int ncs,
                    hipStream_t st);
 int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *g, float seed_scale, const float *z,
@@ -48,16 +65,15 @@ size_t reduce_gpart_ws_bytes(int MP);
 int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
                                float *P, float *v, const int *active, int C, int ncs, hipStream_t st);
 int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
-                       const float *carry_in, const float *zin, float *out, uint32_t *chain_bits, uint32_t *norm_bits,
-                       const int *active, int C, int ncs,
-                       hipStream_t st);
+                       const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
+                       const int *active, int C, int ncs, hipStream_t st);
 
 // shallow PLRNN
 size_t sh_resjac_lds(int M, int L);
 size_t sh_jacform_lds(int M, int L);
 size_t sh_grads_part_floats(int M, int L, int *nblocks);
-int launch_resjac_shplrnn(const ShArgs &a, const float *z, float *F, float *r, uint32_t *masks, const int *active,
-                          hipStream_t st);
+int launch_resjac_shplrnn(const ShArgs &a, const float *z, const float *zalt, const int *zsel, float *F, float *r,
+                          uint32_t *masks, const int *active, hipStream_t st);
 int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, const int *active, const float *gamma,
                            hipStream_t st);
 int launch_grads_shplrnn(const ShArgs &a, const float *z, const float *lam, const uint32_t *masks, float *part,

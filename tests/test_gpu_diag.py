@@ -87,8 +87,10 @@ def test_diag_fused_projection_and_fused_gradients(B, T, M, K):
     assert rel_inf(_c(dB), gr["Bc"]) < TOL
     out2 = D.deer_adjoint(m, x, res["z"], 0.0, 0, g=gt, want_lam=False)
     assert out2["lam"] is None
-    assert np.array_equal(out2["grads"]["lam"].cpu().numpy(), dl)
-    assert np.array_equal(out2["grads"]["Bc"].cpu().numpy(), dB)
+    # the look-back scan combines predecessor values in an order that depends on timing, so
+    # two runs agree to rounding, not bit for bit
+    assert rel_inf(out2["grads"]["lam"].cpu().numpy(), dl.astype(np.float64)) < 1e-5
+    assert rel_inf(out2["grads"]["Bc"].cpu().numpy(), dB.astype(np.float64)) < 1e-5
 
 
 def _readout_params(M, H, No, rng):

@@ -23,6 +23,9 @@ FLAGS = [
     "-ffp-contract=off",
     # no packed-fp32 VALU instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core accumulators in ordinary VGPRs: the chunk kernels apply VALU operations to
+    # them every step, which would otherwise cost two accumulator moves per element
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-Wno-unused-result",
 ]
 

@@ -143,16 +143,18 @@ static int chunk_override() {
 }
 
 // Chunk length of the dense scans: enough chains to fill the machine (about 2048 waves),
-// and a bounded number of chunks per sequence so that the carry pass stays short: 128 with
-// the single-level carry (MP = 64), 1024 with the two-level carry (MP <= 32).
+// and a bounded number of chunks per sequence so that the two-level carry pass stays short
+// (1024 for MP <= 32, 512 for MP = 64, whose group pass composes 64 x 64 maps).
 static int choose_chunk(int B, int T, int MP) {
     const int ov = chunk_override();
     if (ov > 0) return ov < T ? ov : T;
     const long total = (long)B * T;
-    const long target_chains = 2048L * (64 / MP);
+    // MP = 64 runs one chain per wave at two waves per SIMD: 8192 chains keep the tail of a
+    // pass (fewer active sequences) spread over the machine
+    const long target_chains = MP == 64 ? 8192L : 2048L * (64 / MP);
     long C = (total + target_chains - 1) / target_chains;
     if (C < 16) C = 16;
-    const long maxc = MP <= 32 ? 1024 : 128;
+    const long maxc = MP <= 32 ? 1024 : 512;
     const long minC = (T + maxc - 1) / maxc;
     if (C < minC) C = minC;
     if (C > T) C = T;

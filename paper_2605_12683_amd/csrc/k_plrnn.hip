@@ -514,6 +514,171 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
 }
 
 // ---------------------------------------------------------------------------------------
+// The same forward Newton pass for M = 64 when every latent has the same forcing factor p
+// (N = 0 or N = M).  Then the forced Jacobian factors as
+//   J~_t = gp (diag(A) + W diag(m_t)),   gp = gamma p,
+// so W itself (unscaled, in LDS) serves the matrix-core A operand, the residual F and the
+// chunk-local solution, and no M x M operand lives in registers: the kernel fits two waves per
+// SIMD, and one wave's VALU/LDS phase overlaps the other's matrix-core phase.  The scalar gp
+// is applied to the chunk product every 8 steps (acc *= gp^8) instead of every step.
+// One chain per wave (64 lanes = 64 latents for the lane-per-row part).
+// ---------------------------------------------------------------------------------------
+__device__ __forceinline__ float lds_row_dot64(const float (*wl)[68], int row, const float *vec) {
+    const float4 *w4 = reinterpret_cast<const float4 *>(wl[row]);
+    const float4 *v4 = reinterpret_cast<const float4 *>(vec);
+    float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+    for (int q = 0; q < 16; q += 2) {
+        const float4 w0 = w4[q], x0 = v4[q], w1 = w4[q + 1], x1 = v4[q + 1];
+        a0 = fmaf(w0.x, x0.x, a0); a0 = fmaf(w0.y, x0.y, a0); a0 = fmaf(w0.z, x0.z, a0); a0 = fmaf(w0.w, x0.w, a0);
+        a1 = fmaf(w1.x, x1.x, a1); a1 = fmaf(w1.y, x1.y, a1); a1 = fmaf(w1.z, x1.z, a1); a1 = fmaf(w1.w, x1.w, a1);
+    }
+    return a0 + a1;
+}
+
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_newton_product_plrnn64u(
+    const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
+    const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
+    const int *__restrict__ zsel, float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout,
+    float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
+    int ncs) {
+    constexpr int MP = 64, NI = 4, NS = 16;
+    __shared__ __align__(16) float wl[MP][68];
+    __shared__ __align__(16) float lds[64];
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int id = blockIdx.x;
+    const bool ok0 = id < B * ncs;
+    const int b = ok0 ? id / ncs : 0, s0 = ok0 ? (id % ncs) * C : 0;
+    const bool ok = ok0 && (!active || active[b]);
+    const int len = ok ? min(C, T - s0) : 0;
+    for (int e = lane; e < MP * MP; e += 64) {
+        const int row = e / MP, col = e % MP;
+        wl[row][col] = (row < M && col < M) ? W[row * M + col] : 0.f;
+    }
+    const float p = N > 0 ? __fsub_rn(1.0f, alpha) : 1.0f;
+    const float gp = (gamma ? gamma[b] : 1.f) * p;
+    const float gp2 = gp * gp, gp4 = gp2 * gp2, gp8 = gp4 * gp4;
+    float dA[NI][4];
+#pragma unroll
+    for (int I = 0; I < NI; ++I)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * I + 4 * g + r;
+            dA[I][r] = row < M ? A[row] : 0.f;
+        }
+    v4f acc[NI][4];
+#pragma unroll
+    for (int Jt = 0; Jt < 4; ++Jt)
+#pragma unroll
+        for (int I = 0; I < NI; ++I)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[I][Jt][r] = (16 * I + 4 * g + r == 16 * Jt + c) ? 1.f : 0.f;
+    // lane-per-row part: lane = latent
+    const int ui = lane;
+    const bool lat = ui < M;
+    const float Ai = lat ? A[ui] : 0.f, hi = (lat && h) ? h[ui] : 0.f;
+    const bool forced = ui < N;
+    const float *z = cur_iter(zbuf, zalt, zsel, b);
+    float zprev = 0.f;
+    if (len > 0 && lat) {
+        if (s0 == 0) zprev = z0 ? z0[(size_t)b * M + ui] : (forced ? x[(size_t)b * (T + 1) * N + ui] : 0.f);
+        else zprev = z[((size_t)b * T + s0 - 1) * M + ui];
+    }
+    float u = 0.f;
+    float zn = 0.f, xn = 0.f;
+    if (len > 0 && lat) {
+        zn = z[((size_t)b * T + s0) * M + ui];
+        if (forced) xn = x[((size_t)b * (T + 1) + s0) * N + ui];
+    }
+    lds_barrier();   // W in LDS
+    const int maxlen = __builtin_amdgcn_readfirstlane(len);
+    for (int t = 0; t < maxlen; ++t) {
+        const bool run = lat;
+        const int s = s0 + t;
+        const float zcur = zn, xb = xn;
+        if (t + 1 < len && lat) {
+            zn = z[((size_t)b * T + s + 1) * M + ui];
+            if (forced) xn = x[((size_t)b * (T + 1) + s + 1) * N + ui];
+        }
+        float zt = 0.f;
+        if (run) {
+            if (s == 0 || !forced) zt = zprev;
+            else zt = __fadd_rn(__fmul_rn(p, zprev), __fmul_rn(alpha, xb));
+        }
+        const bool pos = zt > 0.f;
+        const uint64_t bal = __ballot(pos);
+        lds[lane] = pos ? zt : 0.f;
+        lds_barrier();
+        const float F = fmaf(Ai, zt, lds_row_dot64(wl, ui, lds)) + hi;
+        lds_barrier();
+        const float r = zcur - F;
+        if (run) {
+            r_out[((size_t)b * T + s) * M + ui] = r;
+            if (ui == 0) {
+                const size_t step = (size_t)b * T + s;
+                masks[step * 2] = (uint32_t)bal;
+                if (M > 32) masks[step * 2 + 1] = (uint32_t)(bal >> 32);
+            }
+        }
+        // P <- (diag(A) + W diag(m)) P   (the factor gp is applied every 8 steps)
+        const uint32_t w0 = (uint32_t)bal, w1 = (uint32_t)(bal >> 32);
+#pragma unroll
+        for (int Jt = 0; Jt < 4; ++Jt) {
+            float Bop[NS];
+#pragma unroll
+            for (int j = 0; j < NS / 4; ++j) {
+                const uint32_t wj = (j >> 1) ? w1 : w0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) Bop[4 * j + q] = select_bit(wj, 16 * (j & 1) + 4 * g + q, acc[j][Jt][q]);
+            }
+#pragma unroll
+            for (int I = 0; I < NI; ++I)
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) acc[I][Jt][r2] *= dA[I][r2];
+#pragma unroll
+            for (int I = 0; I < NI; ++I)
+#pragma unroll
+                for (int j = 0; j < NS / 4; ++j) {
+                    const float4 a4 = *reinterpret_cast<const float4 *>(&wl[16 * I + c][16 * j + 4 * g]);
+                    acc[I][Jt] = mfma16x16x4(a4.x, Bop[4 * j + 0], acc[I][Jt]);
+                    acc[I][Jt] = mfma16x16x4(a4.y, Bop[4 * j + 1], acc[I][Jt]);
+                    acc[I][Jt] = mfma16x16x4(a4.z, Bop[4 * j + 2], acc[I][Jt]);
+                    acc[I][Jt] = mfma16x16x4(a4.w, Bop[4 * j + 3], acc[I][Jt]);
+                }
+        }
+        if ((t & 7) == 7) {
+#pragma unroll
+            for (int Jt = 0; Jt < 4; ++Jt)
+#pragma unroll
+                for (int I = 0; I < NI; ++I)
+#pragma unroll
+                    for (int r2 = 0; r2 < 4; ++r2) acc[I][Jt][r2] *= gp8;
+        }
+        // chunk-local solution: u <- gp (A o u + W (m o u)) - r
+        lds[lane] = pos ? u : 0.f;
+        lds_barrier();
+        const float y = fmaf(Ai, u, lds_row_dot64(wl, ui, lds));
+        lds_barrier();
+        if (run) {
+            u = fmaf(gp, y, -r);
+            zprev = zcur;
+        }
+    }
+    if (ok0 && len > 0) {
+        float rest = 1.f;
+        for (int k = 0; k < (len & 7); ++k) rest *= gp;
+        float *P = Pout + (size_t)id * MP * MP;
+#pragma unroll
+        for (int Jt = 0; Jt < 4; ++Jt)
+#pragma unroll
+            for (int I = 0; I < NI; ++I)
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) P[(16 * I + 4 * g + r2) * MP + 16 * Jt + c] = acc[I][Jt][r2] * rest;
+    }
+    if (ok0) vout[(size_t)id * MP + ui] = u;
+}
+
+// ---------------------------------------------------------------------------------------
 // carries across chunks
 //   forward: carry_in[c] = y_end(c-1),  y_end(c) = P_c y_end(c-1) + v_c
 //   reverse: carry_in[c] = lam_{s1(c)}, lam_{s0(c)} = P_c^T lam_{s1(c)} + v_c
@@ -623,7 +788,7 @@ __global__ __launch_bounds__(256) void k_carry_group(const float *__restrict__ P
             float acc = 0.f;
             if (e < MP * MP) {
                 const int r = e / MP, col = e % MP;
-#pragma unroll
+#pragma unroll(MP <= 32 ? MP : 8)
                 for (int k = 0; k < MP; ++k) acc = fmaf(Am[r][k], Q[k][col], acc);
             }
             qn[t] = acc;
@@ -1041,15 +1206,18 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
 #define NP(MPV)                                                                                                   \
     hipLaunchKernelGGL(k_newton_product_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, \
                        a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs)
-    if (MP == 16) NP(16); else if (MP == 32) NP(32); else NP(64);
+    if (MP == 64 && (a.N == 0 || a.N == a.M)) {   // uniform forcing factor: W-in-LDS kernel
+        hipLaunchKernelGGL(k_newton_product_plrnn64u, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0,
+                           z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
+    } else if (MP == 16) NP(16); else if (MP == 32) NP(32); else NP(64);
 #undef NP
     DEER_LAUNCH_CHECK("k_newton_product_plrnn");
     return DEER_OK;
 }
 
-// two-level carry for chunk sequences at least this long (MP <= 32)
+// two-level carry for chunk sequences at least this long
 static int carry_group_size(int MP, int ncs) {
-    if (MP > 32 || ncs < 96) return 0;
+    if (ncs < 96) return 0;
     int G = 8;
     while (2 * G * G < ncs) G <<= 1;   // a group step costs about twice a walk step
     return G;
@@ -1086,17 +1254,15 @@ int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_
         float *gu = gq + (size_t)B * ng * MP * MP;
         float *gc = gu + (size_t)B * ng * MP;
         const int grid = B * ng;
-        if (MP == 16) {
-            if (rev) CG(16, true, grid); else CG(16, false, grid);
-            CA(16, false, gq, gu, gc, nullptr, ng, ng, nullptr, B);
-            if (rev) CA(16, true, P, v, carry_in, norm_bits, ncs, G, gc, grid);
-            else CA(16, false, P, v, carry_in, norm_bits, ncs, G, gc, grid);
-        } else {
-            if (rev) CG(32, true, grid); else CG(32, false, grid);
-            CA(32, false, gq, gu, gc, nullptr, ng, ng, nullptr, B);
-            if (rev) CA(32, true, P, v, carry_in, norm_bits, ncs, G, gc, grid);
-            else CA(32, false, P, v, carry_in, norm_bits, ncs, G, gc, grid);
-        }
+#define CG3(MPV)                                                             \
+    {                                                                        \
+        if (rev) CG(MPV, true, grid); else CG(MPV, false, grid);             \
+        CA(MPV, false, gq, gu, gc, nullptr, ng, ng, nullptr, B);             \
+        if (rev) CA(MPV, true, P, v, carry_in, norm_bits, ncs, G, gc, grid); \
+        else CA(MPV, false, P, v, carry_in, norm_bits, ncs, G, gc, grid);    \
+    }
+        if (MP == 16) CG3(16) else if (MP == 32) CG3(32) else CG3(64)
+#undef CG3
     }
 #undef CG
 #undef CA

@@ -147,6 +147,142 @@ __global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restr
     }
 }
 
+// Forward chunk product with the chunk-local solution on the matrix cores as well: per chain
+// the B operand is [P | u] (P's MP/16 column tiles plus one tile whose column 0 is u and whose
+// other columns stay 0), so one set of A fragments J~_t advances both
+//   P <- J~_t P,   u <- J~_t u + rhs_sign * rhs_t,
+// and neither LDS nor barriers are needed.  The A fragments are read one step ahead; with the
+// k-permutation kappa(4j+q, g) = 16j + 4g + q the four values a lane needs for k-steps 4j..4j+3
+// are one 16-byte vector of row 16I + c.
+template <int MP>
+__global__ __launch_bounds__(64) void k_chunk_product_dense_fwd(const float *__restrict__ J,
+                                                                const float *__restrict__ rhs, float rhs_sign,
+                                                                float *__restrict__ Pout, float *__restrict__ vout,
+                                                                const int *__restrict__ active, int B, int T, int M,
+                                                                int C, int ncs) {
+    using G = DGeo<MP>;
+    constexpr int NCH = G::NCH, NI = G::NI, NS = G::NS, PT = MP / 16;
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int nchains = B * ncs;
+    const int chain0 = blockIdx.x * NCH;
+    int pb[NCH], plo[NCH], plen[NCH];
+    int maxlen = 0;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n) {
+        const int id = chain0 + n;
+        bool ok = id < nchains;
+        const int b = ok ? id / ncs : 0, cc = ok ? id % ncs : 0;
+        ok = ok && (!active || active[b]);
+        const int s0 = cc * C, s1 = min(s0 + C, T);
+        pb[n] = b;
+        plo[n] = s0;
+        plen[n] = ok ? max(s1 - s0, 0) : 0;
+        maxlen = max(maxlen, plen[n]);
+    }
+    const bool vec = (M == MP);   // full 16-byte rows, no padding
+    v4f acc[NCH][PT + 1][NI];
+#pragma unroll
+    for (int n = 0; n < NCH; ++n)
+#pragma unroll
+        for (int tt = 0; tt <= PT; ++tt)
+#pragma unroll
+            for (int I = 0; I < NI; ++I)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    acc[n][tt][I][r] = (tt < PT && 16 * I + 4 * g + r == 16 * tt + c) ? 1.f : 0.f;
+    float an[NCH][NI][NS];   // A fragments of the next step
+    float rn[NCH][NI][4];    // right-hand side of the next step (lanes of column 0)
+    auto fetch = [&](int t) {
+#pragma unroll
+        for (int n = 0; n < NCH; ++n) {
+            const bool run = t < plen[n];
+            const size_t step = (size_t)pb[n] * T + plo[n] + t;
+            const float *Jp = J + step * M * M;
+#pragma unroll
+            for (int I = 0; I < NI; ++I) {
+#pragma unroll
+                for (int j = 0; j < NS / 4; ++j) {
+                    if (vec) {
+                        const float4 v4 = run ? *reinterpret_cast<const float4 *>(Jp + (16 * I + c) * M + 16 * j + 4 * g)
+                                              : make_float4(0.f, 0.f, 0.f, 0.f);
+                        an[n][I][4 * j] = v4.x;
+                        an[n][I][4 * j + 1] = v4.y;
+                        an[n][I][4 * j + 2] = v4.z;
+                        an[n][I][4 * j + 3] = v4.w;
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            an[n][I][4 * j + q] = run ? jload(Jp, M, 16 * I + c, 16 * j + 4 * g + q) : 0.f;
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = 16 * I + 4 * g + r;
+                    rn[n][I][r] = (run && c == 0 && row < M) ? rhs[step * M + row] : 0.f;
+                }
+            }
+        }
+    };
+    fetch(0);
+    for (int t = 0; t < maxlen; ++t) {
+        float ac[NCH][NI][NS], rc[NCH][NI][4];
+#pragma unroll
+        for (int n = 0; n < NCH; ++n)
+#pragma unroll
+            for (int I = 0; I < NI; ++I) {
+#pragma unroll
+                for (int s = 0; s < NS; ++s) ac[n][I][s] = an[n][I][s];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) rc[n][I][r] = rn[n][I][r];
+            }
+        fetch(t + 1);
+#pragma unroll
+        for (int n = 0; n < NCH; ++n) {
+            if (t < plen[n]) {
+#pragma unroll
+                for (int tt = 0; tt <= PT; ++tt) {
+                    float Bop[NS];
+#pragma unroll
+                    for (int j = 0; j < NS / 4; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) Bop[4 * j + q] = acc[n][tt][j][q];
+#pragma unroll
+                    for (int I = 0; I < NI; ++I) {
+                        v4f a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                        for (int s = 0; s < NS; ++s) a = mfma16x16x4(ac[n][I][s], Bop[s], a);
+                        acc[n][tt][I] = a;
+                    }
+                }
+#pragma unroll
+                for (int I = 0; I < NI; ++I)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[n][PT][I][r] = fmaf(rhs_sign, rc[n][I][r], acc[n][PT][I][r]);
+            }
+        }
+    }
+#pragma unroll
+    for (int n = 0; n < NCH; ++n) {
+        const int id = chain0 + n;
+        if (id >= nchains) continue;
+        if (plen[n] > 0) {
+            float *P = Pout + (size_t)id * MP * MP;
+#pragma unroll
+            for (int tt = 0; tt < PT; ++tt)
+#pragma unroll
+                for (int I = 0; I < NI; ++I)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) P[(16 * I + 4 * g + r) * MP + 16 * tt + c] = acc[n][tt][I][r];
+        }
+        if (c == 0) {
+#pragma unroll
+            for (int I = 0; I < NI; ++I)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) vout[(size_t)id * MP + 16 * I + 4 * g + r] = acc[n][PT][I][r];
+        }
+    }
+}
+
 // MODE 0: forward Newton fix-up (next iterate = current + Delta, in place when the two buffers
 //         coincide; per-chain max |Delta| and max |z|)
 // MODE 1: forward bare scan (y written)
@@ -260,11 +396,15 @@ int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, co
 #define CPD(MPV, R)                                                                                            \
     hipLaunchKernelGGL((k_chunk_product_dense<MPV, R>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, P, v, active, \
                        B, T, M, C, ncs)
+#define CPF(MPV)                                                                                           \
+    hipLaunchKernelGGL((k_chunk_product_dense_fwd<MPV>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, P, v, \
+                       active, B, T, M, C, ncs)
     if (!rev) {
-        if (MP == 16) CPD(16, false); else if (MP == 32) CPD(32, false); else CPD(64, false);
+        if (MP == 16) CPF(16); else if (MP == 32) CPF(32); else CPF(64);
     } else {
         if (MP == 16) CPD(16, true); else if (MP == 32) CPD(32, true); else CPD(64, true);
     }
+#undef CPF
 #undef CPD
     DEER_LAUNCH_CHECK("k_chunk_product_dense");
     return DEER_OK;

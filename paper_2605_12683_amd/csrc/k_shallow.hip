@@ -18,30 +18,41 @@ namespace deer {
 __device__ __forceinline__ float p_at(int i, int N, float alpha) { return i < N ? __fsub_rn(1.0f, alpha) : 1.0f; }
 
 // ---------------------------------------------------------------------------------------
-// residual + masks.  Block of 256 threads, TT rows (b, t) per tile, grid-stride over tiles.
-// dynamic LDS: zt[TT][M] | ru[TT][L] | W1T[L][M] (W1 transposed)
+// residual + masks.  Block of 256 threads (4 waves), TT rows (b, t) per tile, grid-stride
+// over tiles.  The hidden pre-activations u = W2 z~ + h2 that decide the masks are summed on
+// the VALU in a fixed order (left to right from h2, a rounding after every multiply and add);
+// F = A z~ + W1 relu(u) + h1 is a [M x L] x [L x TT] product on the matrix cores with the
+// k range split over the 4 waves and the partial tiles summed through LDS.
+// dynamic LDS: zt[TT][MP] | ru[TT][LQ] | W1[MP][LQ] | partial F tiles [4][NI][64][4]
+// (LQ = L rounded up to 16, + 4 so that rows stay 16-byte aligned and spread over banks)
 // ---------------------------------------------------------------------------------------
 constexpr int SH_TT = 16;
+
+static __host__ __device__ inline int sh_LQ(int L) { return (L + 15) / 16 * 16 + 4; }
 
 template <int MP>
 __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const float *zbuf, const float *zalt,
                                                         const int *__restrict__ zsel, float *__restrict__ F_out,
                                                         float *__restrict__ r_out, uint32_t *__restrict__ masks,
                                                         const int *__restrict__ active) {
+    constexpr int NI = MP / 16;
     extern __shared__ __align__(16) float smem[];
-    const int M = a.M, L = a.L, T = a.T;
+    const int M = a.M, L = a.L, T = a.T, LQ = sh_LQ(L);
     float *zt = smem;                    // [SH_TT][MP], zero padded
-    float *ru = zt + SH_TT * MP;         // [SH_TT][L]
-    float *w1t = ru + SH_TT * L;         // [L][M]
+    float *ru = zt + SH_TT * MP;         // [SH_TT][LQ], zero padded
+    float *w1s = ru + SH_TT * LQ;        // [MP][LQ] = W1, zero padded
+    v4f *red = reinterpret_cast<v4f *>(w1s + MP * LQ);   // [4][NI][64]
     const int tid = threadIdx.x;
-    const int lane = tid & 63;
+    const int lane = tid & 63, wv = tid >> 6, g = lane >> 4, c = lane & 15;
     const int LW = (L + 31) / 32;
-    for (int e = tid; e < L * M; e += 256) {
-        const int l = e / M, i = e % M;
-        w1t[e] = a.W1[i * L + l];
+    for (int e = tid; e < MP * LQ; e += 256) {
+        const int i = e / LQ, l = e % LQ;
+        w1s[e] = (i < M && l < L) ? a.W1[i * L + l] : 0.f;
     }
+    for (int e = tid; e < SH_TT * LQ; e += 256) ru[e] = 0.f;
     const long total = (long)a.B * T;
     const long ntiles = (total + SH_TT - 1) / SH_TT;
+    const int njg = (L + 15) / 16;
     for (long tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const long row0 = tile * SH_TT;
         __syncthreads();
@@ -65,17 +76,21 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
 #pragma unroll
             for (int k = 0; k < MP; ++k) w2r[k] = (jok && k < M) ? a.W2[(size_t)j * M + k] : 0.f;
             const float h2j = (jok && a.h2) ? a.h2[j] : 0.f;
-            for (int tt0 = 0; tt0 < SH_TT; tt0 += 4) {
-                float u[4] = {h2j, h2j, h2j, h2j};
+            // RG rows at a time: independent chains interleaved (each sum is serial in k)
+            constexpr int RG = 4;
+            for (int tt0 = 0; tt0 < SH_TT; tt0 += RG) {
+                float u[RG];
+#pragma unroll
+                for (int q = 0; q < RG; ++q) u[q] = h2j;
 #pragma unroll
                 for (int k = 0; k < MP; ++k)
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) u[q] = __fadd_rn(u[q], __fmul_rn(w2r[k], zt[(tt0 + q) * MP + k]));
+                    for (int q = 0; q < RG; ++q) u[q] = __fadd_rn(u[q], __fmul_rn(w2r[k], zt[(tt0 + q) * MP + k]));
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
+                for (int q = 0; q < RG; ++q) {
                     const int tt = tt0 + q;
                     const bool pos = jok && u[q] > 0.f;
-                    if (jok) ru[tt * L + j] = pos ? u[q] : 0.f;
+                    if (jok) ru[tt * LQ + j] = pos ? u[q] : 0.f;
                     const uint64_t bal = __ballot(pos);
                     const long row = row0 + tt;
                     if (masks && row < total && (lane == 0 || lane == 32)) {
@@ -89,26 +104,50 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
             }
         }
         __syncthreads();
-        // F and r: thread -> (tt, i)
-        for (int e = tid; e < SH_TT * M; e += 256) {
-            const int tt = e / M, i = e % M;
-            const long row = row0 + tt;
-            if (row >= total) continue;
-            const int b = (int)(row / T);
-            if (active && !active[b]) continue;
-            const float *rr = ru + tt * L;
-            float acc0 = 0.f, acc1 = 0.f;
-            int l = 0;
-            for (; l + 1 < L; l += 2) {
-                acc0 = fmaf(w1t[l * M + i], rr[l], acc0);
-                acc1 = fmaf(w1t[(l + 1) * M + i], rr[l + 1], acc1);
+        // F^T tile [MP x 16 rows] = W1 relu(U)^T, this wave's share of the k range; lane (g, c)
+        // ends with F^T[16I + 4g + r][row c]; k-step (jg, q) uses k = 16 jg + 4g + q in group g
+        v4f fa[NI];
+#pragma unroll
+        for (int I = 0; I < NI; ++I) fa[I] = (v4f){0.f, 0.f, 0.f, 0.f};
+        for (int jg = wv; jg < njg; jg += 4) {
+            const float4 bq = *reinterpret_cast<const float4 *>(ru + c * LQ + 16 * jg + 4 * g);
+#pragma unroll
+            for (int I = 0; I < NI; ++I) {
+                const float4 aq = *reinterpret_cast<const float4 *>(w1s + (16 * I + c) * LQ + 16 * jg + 4 * g);
+                fa[I] = mfma16x16x4(aq.x, bq.x, fa[I]);
+                fa[I] = mfma16x16x4(aq.y, bq.y, fa[I]);
+                fa[I] = mfma16x16x4(aq.z, bq.z, fa[I]);
+                fa[I] = mfma16x16x4(aq.w, bq.w, fa[I]);
             }
-            if (l < L) acc0 = fmaf(w1t[l * M + i], rr[l], acc0);
-            const float ztv = zt[tt * MP + i];
-            const float F = fmaf(a.A[i], ztv, acc0 + acc1) + (a.h1 ? a.h1[i] : 0.f);
-            const size_t e2 = (size_t)row * M + i;
-            if (F_out) F_out[e2] = F;
-            if (r_out) r_out[e2] = cur_iter(zbuf, zalt, zsel, (int)(row / a.T))[e2] - F;
+        }
+#pragma unroll
+        for (int I = 0; I < NI; ++I) red[(wv * NI + I) * 64 + lane] = fa[I];
+        __syncthreads();
+        if (wv == 0) {
+            const long row = row0 + c;
+            const bool rok = row < total && (!active || active[row / T]);
+            if (rok) {
+                const float *zc = cur_iter(zbuf, zalt, zsel, (int)(row / T));
+#pragma unroll
+                for (int I = 0; I < NI; ++I) {
+                    v4f sum = red[I * 64 + lane];
+#pragma unroll
+                    for (int w = 1; w < 4; ++w) {
+                        const v4f o = red[(w * NI + I) * 64 + lane];
+                        sum[0] += o[0]; sum[1] += o[1]; sum[2] += o[2]; sum[3] += o[3];
+                    }
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int i = 16 * I + 4 * g + r;
+                        if (i < M) {
+                            const float F = fmaf(a.A[i], zt[c * MP + i], sum[r]) + (a.h1 ? a.h1[i] : 0.f);
+                            const size_t e2 = (size_t)row * M + i;
+                            if (F_out) F_out[e2] = F;
+                            if (r_out) r_out[e2] = zc[e2] - F;
+                        }
+                    }
+                }
+            }
         }
     }
 }
@@ -349,7 +388,10 @@ __global__ void k_mse_seed(const float *__restrict__ z, const float *__restrict_
 // ---------------------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------------------
-size_t sh_resjac_lds(int M, int L) { return (size_t)(SH_TT * padded_dim(M) + SH_TT * L + L * M) * sizeof(float); }
+size_t sh_resjac_lds(int M, int L) {
+    const int MP = padded_dim(M), LQ = sh_LQ(L);
+    return (size_t)(SH_TT * MP + SH_TT * LQ + MP * LQ + 4 * (MP / 16) * 64 * 4) * sizeof(float);
+}
 
 static int sh_LP(int L) { return (L + 15) / 16 * 16; }
 

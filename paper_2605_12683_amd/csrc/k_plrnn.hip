@@ -12,6 +12,8 @@
 //                      gradient partial sums (gradients appendix)
 //
 // Padded dimension MP in {16, 32, 64} (the next one >= M); a wave holds NCH = 64/MP chains.
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 
@@ -514,6 +516,388 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
 }
 
 // ---------------------------------------------------------------------------------------
+// M <= 16: register-tiled forward Newton pass and fix-up.
+// A wave holds four chains, one per 16-lane row (lane = 16 * chain + latent), so a row of the
+// wave is one chain's state vector and the products W y of F and of the chunk-local solution
+// are formed with DPP row rotations (no LDS, no barrier).  Steps go in tiles of TB.  In a tile
+// that all four chains run to its end (every tile but a ragged chunk's last) all loads of the
+// tile are issued at once through buffer resources (one lane offset for all of them), the
+// residual of every step of the tile, which does not depend on the recurrence, is formed and
+// stored first, and the serial part then runs from registers, with the matrix-core updates of
+// the four chains free of branches so that they interleave.  Other tiles go step by step.
+// ---------------------------------------------------------------------------------------
+
+// lane l of each 16-lane row receives v from lane row_src(l, K) of the same row
+template <int K>
+__device__ __forceinline__ float row_ror(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + K, 0xF, 0xF, true));
+}
+template <int K>
+__device__ __forceinline__ int row_ror_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, 0x120 + K, 0xF, 0xF, true);
+}
+
+// source lane (within the row) of rotation k, k = 0..15
+__device__ __forceinline__ void row_sources(int c, int (&src)[16]) {
+    src[0] = c;
+    src[1] = row_ror_i<1>(c);   src[2] = row_ror_i<2>(c);   src[3] = row_ror_i<3>(c);
+    src[4] = row_ror_i<4>(c);   src[5] = row_ror_i<5>(c);   src[6] = row_ror_i<6>(c);
+    src[7] = row_ror_i<7>(c);   src[8] = row_ror_i<8>(c);   src[9] = row_ror_i<9>(c);
+    src[10] = row_ror_i<10>(c); src[11] = row_ror_i<11>(c); src[12] = row_ror_i<12>(c);
+    src[13] = row_ror_i<13>(c); src[14] = row_ror_i<14>(c); src[15] = row_ror_i<15>(c);
+}
+
+// sum_k w[k] * v(row_src(lane, k)): with w[k] = W[i][row_src(i, k)] this is (W v)_i for the
+// vector v held by the 16 lanes of the row
+__device__ __forceinline__ float row16_dot(const float (&w)[16], float v) {
+    // the rotated operand first: it is the one a DPP-modified multiply-add can take
+    float a0 = v * w[0], a1 = row_ror<1>(v) * w[1];
+    a0 = fmaf(row_ror<2>(v), w[2], a0);   a1 = fmaf(row_ror<3>(v), w[3], a1);
+    a0 = fmaf(row_ror<4>(v), w[4], a0);   a1 = fmaf(row_ror<5>(v), w[5], a1);
+    a0 = fmaf(row_ror<6>(v), w[6], a0);   a1 = fmaf(row_ror<7>(v), w[7], a1);
+    a0 = fmaf(row_ror<8>(v), w[8], a0);   a1 = fmaf(row_ror<9>(v), w[9], a1);
+    a0 = fmaf(row_ror<10>(v), w[10], a0); a1 = fmaf(row_ror<11>(v), w[11], a1);
+    a0 = fmaf(row_ror<12>(v), w[12], a0); a1 = fmaf(row_ror<13>(v), w[13], a1);
+    a0 = fmaf(row_ror<14>(v), w[14], a0); a1 = fmaf(row_ror<15>(v), w[15], a1);
+    return a0 + a1;
+}
+
+// Buffer resource with a wave-uniform base: an access adds a per-lane byte offset (VGPR) and a
+// wave-uniform byte offset (SGPR).  A lane offset of 2^31 or more is outside the resource: a
+// load from it returns zero and a store to it is dropped.
+constexpr uint32_t kOffLane = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t wave_rsrc(const void *base) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ uint32_t bload_u(__amdgpu_buffer_rsrc_t rs, uint32_t voff, int soff) {
+    return __builtin_amdgcn_raw_buffer_load_b32(rs, (int)voff, soff, 0);
+}
+__device__ __forceinline__ float bload(__amdgpu_buffer_rsrc_t rs, uint32_t voff, int soff) {
+    return __uint_as_float(bload_u(rs, voff, soff));
+}
+__device__ __forceinline__ void bstore_u(__amdgpu_buffer_rsrc_t rs, uint32_t v, uint32_t voff, int soff) {
+    __builtin_amdgcn_raw_buffer_store_b32(v, rs, (int)voff, soff, 0);
+}
+
+__device__ __forceinline__ int rfl_i(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ float rfl_f(float v) { return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v))); }
+
+// the wave's four chains: lengths, damping, and whether they all read one iterate buffer
+struct Chains16 {
+    int plen[4];
+    float gam[4];
+    int minlen, maxlen;
+    bool onebuf;
+};
+__device__ __forceinline__ Chains16 chains16(int chain0, int nchains, int ncs, int C, int T,
+                                             const int *__restrict__ active, const float *__restrict__ gamma,
+                                             const int *__restrict__ zsel) {
+    Chains16 w;
+    w.minlen = C;
+    w.maxlen = 0;
+    w.onebuf = true;
+    int sel0 = -1;
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        const int id = chain0 + n;
+        bool ok = id < nchains;
+        const int b = ok ? id / ncs : 0, cc = ok ? id % ncs : 0;
+        ok = ok && (!active || active[b]);
+        w.plen[n] = rfl_i(ok ? min(C, T - cc * C) : 0);
+        w.gam[n] = rfl_f(gamma ? gamma[b] : 1.f);
+        const int sel = rfl_i(zsel ? zsel[b] : 0);
+        if (w.plen[n] > 0) {
+            if (sel0 >= 0 && sel != sel0) w.onebuf = false;
+            sel0 = sel;
+        }
+        w.minlen = min(w.minlen, w.plen[n]);
+        w.maxlen = max(w.maxlen, w.plen[n]);
+    }
+    return w;
+}
+
+// acc[n] *= gamma_n^(steps chain n ran in the tile [t0, t0 + tl)): J~ = gamma (...) per step
+__device__ __forceinline__ void damp_tile(v4f (&acc)[4], const Chains16 &w, int t0, int tl) {
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        const float gm = w.gam[n];
+        if (gm != 1.f) {
+            const int steps = max(0, min(tl, w.plen[n] - t0));
+            float gp = 1.f;
+            for (int k = 0; k < steps; ++k) gp *= gm;
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) acc[n][r2] *= gp;
+        }
+    }
+}
+
+// one matrix-core step of chain n: acc <- (diag(d) + W diag(m)) acc (layout of the MP = 16
+// generic kernel: Aop = columns of W p, dI = rows of diag(A) p)
+__device__ __forceinline__ void mfma_step16(v4f &acc, uint32_t wn, int g, const float (&Aop)[4],
+                                            const float (&dI)[4]) {
+    float Bop[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) Bop[q] = select_bit(wn, 4 * g + q, acc[q]);
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2) acc[r2] *= dI[r2];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc = mfma16x16x4(Aop[q], Bop[q], acc);
+}
+
+template <int TB>
+__global__ __launch_bounds__(64) void k_newton_product_plrnn16(
+    const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
+    const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
+    const int *__restrict__ zsel, float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout,
+    float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
+    int ncs) {
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int nchains = B * ncs;
+    const int chain0 = blockIdx.x * 4;
+    const Chains16 w = chains16(chain0, nchains, ncs, C, T, active, gamma, zsel);
+    if (w.maxlen == 0) return;
+    float Aop[4], dI[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int col = 4 * g + q;
+        Aop[q] = (c < M && col < M) ? W[c * M + col] * p_of(col, N, alpha) : 0.f;
+        dI[q] = col < M ? A[col] * p_of(col, N, alpha) : 0.f;
+    }
+    v4f acc[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[n][r] = (4 * g + r == c) ? 1.f : 0.f;
+    // row part: this lane is latent c of chain g
+    const int id = chain0 + g;
+    const bool okc = id < nchains;
+    const int b = okc ? id / ncs : 0, s0 = okc ? (id % ncs) * C : 0;
+    int len = 0;
+    float ugam = 1.f;
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+        if (n == g) {
+            len = w.plen[n];
+            ugam = w.gam[n];
+        }
+    const bool lat = c < M, forced = c < N;
+    int src[16];
+    row_sources(c, src);
+    float wr[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) wr[k] = (lat && src[k] < M) ? W[c * M + src[k]] : 0.f;
+    const float Ai = lat ? A[c] : 0.f, hi = (lat && h) ? h[c] : 0.f;
+    const float pi = p_of(c, N, alpha), di = Ai * pi;
+    const float *z = cur_iter(zbuf, zalt, zsel, b);
+    float zprev = 0.f;
+    if (len > 0 && lat) {
+        if (s0 == 0) zprev = z0 ? z0[(size_t)b * M + c] : (forced ? x[(size_t)b * (T + 1) * N + c] : 0.f);
+        else zprev = z[((size_t)b * T + s0 - 1) * M + c];
+    }
+    // tile resources, based at the first row of the wave's first chain
+    const int b0 = chain0 / ncs, s00 = (chain0 % ncs) * C;
+    const size_t row0 = (size_t)b0 * T + s00, xrow0 = (size_t)b0 * (T + 1) + s00;
+    const uint32_t drow = (uint32_t)((size_t)b * T + s0 - row0), dxrow = (uint32_t)((size_t)b * (T + 1) + s0 - xrow0);
+    const float *zw = cur_iter(zbuf, zalt, zsel, b0);
+    const auto rz = wave_rsrc(zw + row0 * M), rr = wave_rsrc(r_out + row0 * M), rm = wave_rsrc(masks + row0);
+    const auto rx = wave_rsrc(N > 0 ? x + xrow0 * N : zw);
+    const uint32_t vz = lat ? 4u * (drow * M + c) : kOffLane;
+    const uint32_t vx = forced ? 4u * (dxrow * N + c) : kOffLane;
+    const uint32_t vm = c == 0 ? 4u * drow : kOffLane;
+    float u = 0.f;
+    for (int t0 = 0; t0 < w.maxlen; t0 += TB) {
+        const int tl = min(TB, w.maxlen - t0);
+        if (w.onebuf && t0 + TB <= w.minlen) {
+            float zv[TB], xv[TB];
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                zv[tt] = bload(rz, vz, 4 * (t0 + tt) * M);
+                xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
+            }
+            // residual and masks of every step of the tile; r overwrites zv
+            uint32_t posb = 0u;
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                const int s = s0 + t0 + tt;
+                const float zt =
+                    (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xv[tt]));
+                const bool pos = zt > 0.f;
+                posb |= (pos ? 1u : 0u) << tt;
+                const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
+                zprev = zv[tt];
+                zv[tt] = zv[tt] - F;
+                bstore_u(rr, __float_as_uint(zv[tt]), vz, 4 * (t0 + tt) * M);
+                const uint64_t bal = __ballot(pos);
+                bstore_u(rm, (uint32_t)((bal >> (16 * g)) & 0xffffull), vm, 4 * (t0 + tt));
+            }
+            // serial part: chunk products and chunk-local solutions
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                const bool pos = (posb >> tt) & 1u;
+                const uint64_t bal = __ballot(pos);
+                // the four chains' updates interleaved: k-slice outer, chain inner
+                float Bop[4][4];
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) Bop[n][q] = select_bit((uint32_t)(bal >> (16 * n)), 4 * g + q, acc[n][q]);
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+#pragma unroll
+                    for (int r2 = 0; r2 < 4; ++r2) acc[n][r2] *= dI[r2];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) acc[n] = mfma16x16x4(Aop[q], Bop[n][q], acc[n]);
+                const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
+                u = fmaf(ugam, y, -zv[tt]);
+            }
+        } else {
+            for (int t = t0; t < t0 + tl; ++t) {
+                const bool run = t < len && lat;
+                const int s = s0 + t;
+                float zcur = 0.f, xb = 0.f;
+                if (run) {
+                    zcur = z[((size_t)b * T + s) * M + c];
+                    if (forced && s > 0) xb = x[((size_t)b * (T + 1) + s) * N + c];
+                }
+                float zt = 0.f;
+                if (run) zt = (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xb));
+                const bool pos = zt > 0.f;
+                const uint64_t bal = __ballot(pos);
+                const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
+                const float r = zcur - F;
+                if (t < len) {
+                    const size_t step = (size_t)b * T + s;
+                    if (lat) r_out[step * M + c] = r;
+                    if (c == 0) masks[step] = (uint32_t)((bal >> (16 * g)) & 0xffffull);
+                }
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+                    if (t < w.plen[n]) mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, Aop, dI);
+                const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
+                if (run) {
+                    u = fmaf(ugam, y, -r);
+                    zprev = zcur;
+                }
+            }
+        }
+        damp_tile(acc, w, t0, tl);
+    }
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        const int cid = chain0 + n;
+        if (cid < nchains && w.plen[n] > 0) {
+            float *P = Pout + (size_t)cid * 256;
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) P[(4 * g + r2) * 16 + c] = acc[n][r2];
+        }
+    }
+    if (okc) vout[(size_t)id * 16 + c] = u;
+}
+
+template <int TB>
+__global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restrict__ A, const float *__restrict__ W,
+                                                          float alpha, int N, const uint32_t *__restrict__ masks,
+                                                          const float *__restrict__ r, const float *__restrict__ carry_in,
+                                                          float *zbuf, float *zalt, const int *__restrict__ zsel,
+                                                          uint32_t *__restrict__ chain_bits,
+                                                          const int *__restrict__ active,
+                                                          const float *__restrict__ gamma, int B, int T, int M, int C,
+                                                          int ncs) {
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int nchains = B * ncs;
+    const int chain0 = blockIdx.x * 4;
+    const Chains16 w = chains16(chain0, nchains, ncs, C, T, active, gamma, zsel);
+    if (w.maxlen == 0) return;
+    const int id = chain0 + g;
+    const bool okc = id < nchains;
+    const int b = okc ? id / ncs : 0, s0 = okc ? (id % ncs) * C : 0;
+    int len = 0;
+    float gm = 1.f;
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+        if (n == g) {
+            len = w.plen[n];
+            gm = w.gam[n];
+        }
+    const bool lat = c < M;
+    int src[16];
+    row_sources(c, src);
+    float wp[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) wp[k] = (lat && src[k] < M) ? W[c * M + src[k]] * p_of(src[k], N, alpha) : 0.f;
+    const float d = lat ? A[c] * p_of(c, N, alpha) : 0.f;
+    float D = (len > 0 && lat) ? carry_in[(size_t)id * 16 + c] : 0.f;
+    const float *zin = cur_iter(zbuf, zalt, zsel, b);
+    float *zout = next_iter(zbuf, zalt, zsel, b);
+    const int b0 = chain0 / ncs;
+    const size_t row0 = (size_t)b0 * T + (size_t)(chain0 % ncs) * C;
+    const uint32_t drow = (uint32_t)((size_t)b * T + s0 - row0);
+    const auto rr = wave_rsrc(r + row0 * M), rm = wave_rsrc(masks + row0);
+    const auto rzi = wave_rsrc(cur_iter(zbuf, zalt, zsel, b0) + row0 * M);
+    const auto rzo = wave_rsrc(next_iter(zbuf, zalt, zsel, b0) + row0 * M);
+    const uint32_t vz = lat ? 4u * (drow * M + c) : kOffLane, vm = 4u * drow;
+    uint32_t emax = 0u, zmax = 0u;
+    for (int t0 = 0; t0 < w.maxlen; t0 += TB) {
+        const int tl = min(TB, w.maxlen - t0);
+        if (w.onebuf && t0 + TB <= w.minlen) {
+            float rv[TB], zv[TB];
+            uint32_t mv[TB];
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                rv[tt] = bload(rr, vz, 4 * (t0 + tt) * M);
+                zv[tt] = bload(rzi, vz, 4 * (t0 + tt) * M);
+                mv[tt] = bload_u(rm, vm, 4 * (t0 + tt));
+            }
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                const bool m = (mv[tt] >> c) & 1u;
+                const float y = fmaf(d, D, row16_dot(wp, m ? D : 0.f));
+                D = fmaf(gm, y, -rv[tt]);
+                const float zc = zv[tt];
+                bstore_u(rzo, __float_as_uint(zc + D), vz, 4 * (t0 + tt) * M);
+                const uint32_t ab = abs_bits(D), zb = abs_bits(zc);
+                emax = emax > ab ? emax : ab;
+                zmax = zmax > zb ? zmax : zb;
+            }
+        } else {
+            for (int t = t0; t < t0 + tl; ++t) {
+                const bool run = t < len && lat;
+                const size_t step = (size_t)b * T + s0 + t;
+                float rc = 0.f, zc = 0.f;
+                uint32_t mc = 0u;
+                if (run) {
+                    rc = r[step * M + c];
+                    zc = zin[step * M + c];
+                    mc = masks[step];
+                }
+                const bool m = run && ((mc >> c) & 1u);
+                const float y = fmaf(d, D, row16_dot(wp, m ? D : 0.f));
+                if (run) {
+                    D = fmaf(gm, y, -rc);
+                    zout[step * M + c] = zc + D;
+                    const uint32_t ab = abs_bits(D), zb = abs_bits(zc);
+                    emax = emax > ab ? emax : ab;
+                    zmax = zmax > zb ? zmax : zb;
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) {
+        const uint32_t o = (uint32_t)__shfl_xor((int)emax, off, 64);
+        const uint32_t oz = (uint32_t)__shfl_xor((int)zmax, off, 64);
+        emax = emax > o ? emax : o;
+        zmax = zmax > oz ? zmax : oz;
+    }
+    if (len > 0 && c == 0) {   // per-chain maxima, reduced per sequence by k_seq_max / k_seq_ctl
+        chain_bits[id] = emax;
+        chain_bits[(size_t)nchains + id] = zmax;
+    }
+}
+
+// ---------------------------------------------------------------------------------------
 // The same forward Newton pass for M = 64 when every latent has the same forcing factor p
 // (N = 0 or N = M).  Then the forced Jacobian factors as
 //   J~_t = gp (diag(A) + W diag(m_t)),   gp = gamma p,
@@ -811,6 +1195,122 @@ __global__ __launch_bounds__(256) void k_carry_group(const float *__restrict__ P
     float *q = gq + ((size_t)b * ngroups + j) * MP * MP;
     for (int e = tid; e < MP * MP; e += 256) q[e] = Q[e / MP][e % MP];
     if (tid < MP) gu[((size_t)b * ngroups + j) * MP + tid] = u[tid];
+}
+
+// ---------------------------------------------------------------------------------------
+// M <= 16 carries on the matrix cores, one wave per walk.  A map A_k (P_c or its transpose)
+// is the A operand of four 16x16x4 MFMAs; the vector being walked is column 0 of the B
+// operand, whose accumulator layout is again the next step's B operand, so a step is four
+// dependent MFMAs and no LDS.  The maps of the next PF steps are in flight while a step runs.
+// ---------------------------------------------------------------------------------------
+template <bool REV>
+__device__ __forceinline__ void carry16_fetch(const float *__restrict__ Pc, const float *__restrict__ vc, int g, int c,
+                                              float (&a)[4], float (&vv)[4]) {
+    if (!REV) {
+        const float4 t = *reinterpret_cast<const float4 *>(Pc + c * 16 + 4 * g);
+        a[0] = t.x; a[1] = t.y; a[2] = t.z; a[3] = t.w;
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) a[q] = Pc[(4 * g + q) * 16 + c];
+    }
+    const float4 u = *reinterpret_cast<const float4 *>(vc + 4 * g);
+    vv[0] = u.x; vv[1] = u.y; vv[2] = u.z; vv[3] = u.w;
+}
+
+// walk of the vector: carry_in[c(k)] = cur_k, cur_{k+1} = A_k cur_k + v_{c(k)} (see k_carry)
+template <bool REV>
+__global__ __launch_bounds__(64) void k_carry16(const float *__restrict__ P, const float *__restrict__ v,
+                                               float *__restrict__ carry_in, const int *__restrict__ active,
+                                               uint32_t *__restrict__ norm_bits, int B, int ncs, int G,
+                                               const float *__restrict__ start) {
+    constexpr int PF = 8;
+    const int ngroups = (ncs + G - 1) / G;
+    const int b = blockIdx.x / ngroups, j = blockIdx.x % ngroups;
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    if (norm_bits && j == 0 && lane == 0) {   // [0, B): max|Delta|, [B, 2B): max|z| of the next fix-up
+        norm_bits[b] = 0u;
+        norm_bits[B + b] = 0u;
+    }
+    if (active && !active[b]) return;
+    const int k0 = j * G, k1 = min(k0 + G, ncs);
+    v4f cur;   // column 0: lane (g, 0) holds rows 4g..4g+3; other columns stay zero
+#pragma unroll
+    for (int r = 0; r < 4; ++r) cur[r] = (start && c == 0) ? start[((size_t)b * ngroups + j) * 16 + 4 * g + r] : 0.f;
+    auto chunk = [&](int step) { return REV ? ncs - 1 - step : step; };
+    float a[PF][4], vv[PF][4];
+#pragma unroll
+    for (int d = 0; d < PF; ++d) {
+        const int cc = chunk(min(k0 + d, k1 - 1));
+        carry16_fetch<REV>(P + ((size_t)b * ncs + cc) * 256, v + ((size_t)b * ncs + cc) * 16, g, c, a[d], vv[d]);
+    }
+    for (int k = k0; k < k1; k += PF) {
+#pragma unroll
+        for (int d = 0; d < PF; ++d) {
+            const int step = k + d;
+            if (step >= k1) break;
+            const size_t id = (size_t)b * ncs + chunk(step);
+            if (c == 0) *reinterpret_cast<float4 *>(carry_in + id * 16 + 4 * g) = make_float4(cur[0], cur[1], cur[2], cur[3]);
+            v4f nx = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) nx = mfma16x16x4(a[d][q], cur[q], nx);
+            if (c == 0) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) nx[r] += vv[d][r];
+            }
+            cur = nx;
+            const int cn = chunk(min(step + PF, k1 - 1));
+            carry16_fetch<REV>(P + ((size_t)b * ncs + cn) * 256, v + ((size_t)b * ncs + cn) * 16, g, c, a[d], vv[d]);
+        }
+    }
+}
+
+// group maps in processing order: Q_j = A_{k1-1} ... A_{k0}, u_j = the group's walk from 0
+template <bool REV>
+__global__ __launch_bounds__(64) void k_carry_group16(const float *__restrict__ P, const float *__restrict__ v,
+                                                     float *__restrict__ gq, float *__restrict__ gu,
+                                                     const int *__restrict__ active, int ncs, int G) {
+    constexpr int PF = 8;
+    const int ngroups = (ncs + G - 1) / G;
+    const int b = blockIdx.x / ngroups, j = blockIdx.x % ngroups;
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    if (active && !active[b]) return;
+    const int k0 = j * G, k1 = min(k0 + G, ncs);
+    v4f Q, u = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Q[r] = (4 * g + r == c) ? 1.f : 0.f;
+    auto chunk = [&](int step) { return REV ? ncs - 1 - step : step; };
+    float a[PF][4], vv[PF][4];
+#pragma unroll
+    for (int d = 0; d < PF; ++d) {
+        const int cc = chunk(min(k0 + d, k1 - 1));
+        carry16_fetch<REV>(P + ((size_t)b * ncs + cc) * 256, v + ((size_t)b * ncs + cc) * 16, g, c, a[d], vv[d]);
+    }
+    for (int k = k0; k < k1; k += PF) {
+#pragma unroll
+        for (int d = 0; d < PF; ++d) {
+            const int step = k + d;
+            if (step >= k1) break;
+            v4f nq = {0.f, 0.f, 0.f, 0.f}, nu = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                nq = mfma16x16x4(a[d][q], Q[q], nq);
+                nu = mfma16x16x4(a[d][q], u[q], nu);
+            }
+            if (c == 0) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) nu[r] += vv[d][r];
+            }
+            Q = nq;
+            u = nu;
+            const int cn = chunk(min(step + PF, k1 - 1));
+            carry16_fetch<REV>(P + ((size_t)b * ncs + cn) * 256, v + ((size_t)b * ncs + cn) * 16, g, c, a[d], vv[d]);
+        }
+    }
+    float *q = gq + ((size_t)b * ngroups + j) * 256;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) q[(4 * g + r) * 16 + c] = Q[r];
+    if (c == 0)
+        *reinterpret_cast<float4 *>(gu + ((size_t)b * ngroups + j) * 16 + 4 * g) = make_float4(u[0], u[1], u[2], u[3]);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -1209,7 +1709,14 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
     if (MP == 64 && (a.N == 0 || a.N == a.M)) {   // uniform forcing factor: W-in-LDS kernel
         hipLaunchKernelGGL(k_newton_product_plrnn64u, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0,
                            z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
-    } else if (MP == 16) NP(16); else if (MP == 32) NP(32); else NP(64);
+    } else if (MP == 16) {
+        if (C <= 16)
+            hipLaunchKernelGGL(k_newton_product_plrnn16<16>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
+                               a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
+        else
+            hipLaunchKernelGGL(k_newton_product_plrnn16<32>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
+                               a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
+    } else if (MP == 32) NP(32); else NP(64);
 #undef NP
     DEER_LAUNCH_CHECK("k_newton_product_plrnn");
     return DEER_OK;
@@ -1239,7 +1746,12 @@ int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_
 #define CG(MPV, R, GRID) \
     hipLaunchKernelGGL((k_carry_group<MPV, R>), dim3(GRID), dim3(256), 0, st, P, v, gq, gu, active, ncs, G)
     if (!G) {
-        if (!rev) {
+        if (MP == 16) {
+            if (rev)
+                hipLaunchKernelGGL(k_carry16<true>, dim3(B), dim3(64), 0, st, P, v, carry_in, active, norm_bits, B, ncs, ncs, nullptr);
+            else
+                hipLaunchKernelGGL(k_carry16<false>, dim3(B), dim3(64), 0, st, P, v, carry_in, active, norm_bits, B, ncs, ncs, nullptr);
+        } else if (!rev) {
             if (MP == 16) CA(16, false, P, v, carry_in, norm_bits, ncs, ncs, nullptr, B);
             else if (MP == 32) CA(32, false, P, v, carry_in, norm_bits, ncs, ncs, nullptr, B);
             else CA(64, false, P, v, carry_in, norm_bits, ncs, ncs, nullptr, B);
@@ -1261,7 +1773,15 @@ int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_
         if (rev) CA(MPV, true, P, v, carry_in, norm_bits, ncs, G, gc, grid); \
         else CA(MPV, false, P, v, carry_in, norm_bits, ncs, G, gc, grid);    \
     }
-        if (MP == 16) CG3(16) else if (MP == 32) CG3(32) else CG3(64)
+        if (MP == 16) {
+            if (rev) hipLaunchKernelGGL(k_carry_group16<true>, dim3(grid), dim3(64), 0, st, P, v, gq, gu, active, ncs, G);
+            else hipLaunchKernelGGL(k_carry_group16<false>, dim3(grid), dim3(64), 0, st, P, v, gq, gu, active, ncs, G);
+            hipLaunchKernelGGL(k_carry16<false>, dim3(B), dim3(64), 0, st, gq, gu, gc, active, nullptr, B, ng, ng, nullptr);
+            if (rev)
+                hipLaunchKernelGGL(k_carry16<true>, dim3(grid), dim3(64), 0, st, P, v, carry_in, active, norm_bits, B, ncs, G, gc);
+            else
+                hipLaunchKernelGGL(k_carry16<false>, dim3(grid), dim3(64), 0, st, P, v, carry_in, active, norm_bits, B, ncs, G, gc);
+        } else if (MP == 32) CG3(32) else CG3(64)
 #undef CG3
     }
 #undef CG
@@ -1280,7 +1800,13 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
 #define FX(MPV)                                                                                                       \
     hipLaunchKernelGGL(k_fixup_fwd_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, carry_in, \
                        z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
-    if (MP == 16) FX(16); else if (MP == 32) FX(32); else FX(64);
+#define FX16(TBV)                                                                                              \
+    hipLaunchKernelGGL(k_fixup_fwd_plrnn16<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, \
+                       carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
+    if (MP == 16) {
+        if (C <= 16) FX16(16); else FX16(32);
+    } else if (MP == 32) FX(32); else FX(64);
+#undef FX16
 #undef FX
     DEER_LAUNCH_CHECK("k_fixup_fwd_plrnn");
     return DEER_OK;

@@ -171,6 +171,8 @@ struct NewtonCtl {
     uint32_t *norm_bits;
     uint32_t *chain_bits;   // per-chain maxima [2][B * ncs] before the per-sequence reduction
     float *zalt;            // second iterate buffer [B,T,M]
+    uint32_t *seq;          // kSeqWords per sequence: the fix-up's fused pass-end control
+    bool fused;             // the update takes the pass-end control itself (no k_seq_ctl)
 };
 
 static NewtonCtl carve_ctl(Carver &c, int B, size_t seq_elems, size_t nchains) {
@@ -189,6 +191,7 @@ static NewtonCtl carve_ctl(Carver &c, int B, size_t seq_elems, size_t nchains) {
     n.norm_bits = c.take<uint32_t>(2 * (size_t)B);
     n.chain_bits = c.take<uint32_t>(2 * nchains);
     n.zalt = c.take<float>((size_t)B * seq_elems);
+    n.seq = c.take<uint32_t>((size_t)kSeqWords * B);
     return n;
 }
 
@@ -363,13 +366,13 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
         return DEER_OK;
     }
     const NewtonDev &nd = ctl.nd;
-    if ((rc = launch_ctl_init(nd, B, st))) return rc;
+    if ((rc = launch_ctl_init(nd, ctl.seq, B, st))) return rc;
     int passes = 0, batch = kFirstBatch;
     while (passes < max_iter) {
         const int n = batch < max_iter - passes ? batch : max_iter - passes;
         for (int k = 0; k < n; ++k) {
             if ((rc = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt))) return rc;
-            if ((rc = launch_seq_ctl(ctl.chain_bits, nd, B, ncs, o->tol, bound, kDamp, st))) return rc;
+            if (!ctl.fused && (rc = launch_seq_ctl(ctl.chain_bits, nd, B, ncs, o->tol, bound, kDamp, st))) return rc;
         }
         passes += n;
         DEER_HIP(hipMemcpyAsync(act.data(), nd.act, B * sizeof(int), hipMemcpyDeviceToHost, st));
@@ -432,15 +435,24 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     std::vector<int> act(B, 1), it(B, 0);
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
+    // M <= 16: the fix-up also takes the pass-end control of the adaptive loop
+    NewtonCtl ctl = w.ctl;
+    ctl.fused = w.MP == 16 && o->fixed_iters <= 0;
+    const FusedCtl fc{ctl.nd, ctl.seq, o->tol, o->step_bound == 0.f ? kDefaultStepBound : o->step_bound, kDamp};
     auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za) -> int {
         int r;
-        if ((r = launch_newton_product_plrnn(a, zb, za, zsel, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, st)))
+        // M <= 16: each wave's four chunks are composed in the forward pass, one kernel walks
+        // the composed maps, and the fix-up applies the per-chunk prefix maps
+        const bool wm = w.MP == 16 && w.ncs % 4 == 0;
+        if ((r = launch_newton_product_plrnn(a, zb, za, zsel, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, wm, st)))
             return r;
-        if ((r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, nullptr, B, w.ncs, w.gws, st))) return r;
+        if (wm) r = launch_carry_walk16(w.P, w.v, w.carry, dact, B, w.ncs, st);
+        else r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, nullptr, B, w.ncs, w.gws, st);
+        if (r) return r;
         return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, zb, za, zsel, w.ctl.chain_bits, dact, gam, w.C, w.ncs,
-                                      st);
+                                      wm ? w.P : nullptr, wm ? w.v : nullptr, (ctl.fused && dact) ? &fc : nullptr, st);
     };
-    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ncs, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
+    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ncs, ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
         if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
     }

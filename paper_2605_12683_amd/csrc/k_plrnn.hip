@@ -529,10 +529,6 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
 
 // lane l of each 16-lane row receives v from lane row_src(l, K) of the same row
 template <int K>
-__device__ __forceinline__ float row_ror(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + K, 0xF, 0xF, true));
-}
-template <int K>
 __device__ __forceinline__ int row_ror_i(int v) {
     return __builtin_amdgcn_update_dpp(0, v, 0x120 + K, 0xF, 0xF, true);
 }
@@ -548,19 +544,36 @@ __device__ __forceinline__ void row_sources(int c, int (&src)[16]) {
 }
 
 // sum_k w[k] * v(row_src(lane, k)): with w[k] = W[i][row_src(i, k)] this is (W v)_i for the
-// vector v held by the 16 lanes of the row
+// vector v held by the 16 lanes of the row.  One multiply-add with a DPP row rotation of v per
+// term (the compiler does not fuse a rotation into v_fmac by itself); the leading s_nop covers
+// the wait a DPP read needs after a VALU write of v.  All 64 lanes must be active.
+#define DEER_RR(k) " row_ror:" #k " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
 __device__ __forceinline__ float row16_dot(const float (&w)[16], float v) {
-    // the rotated operand first: it is the one a DPP-modified multiply-add can take
-    float a0 = v * w[0], a1 = row_ror<1>(v) * w[1];
-    a0 = fmaf(row_ror<2>(v), w[2], a0);   a1 = fmaf(row_ror<3>(v), w[3], a1);
-    a0 = fmaf(row_ror<4>(v), w[4], a0);   a1 = fmaf(row_ror<5>(v), w[5], a1);
-    a0 = fmaf(row_ror<6>(v), w[6], a0);   a1 = fmaf(row_ror<7>(v), w[7], a1);
-    a0 = fmaf(row_ror<8>(v), w[8], a0);   a1 = fmaf(row_ror<9>(v), w[9], a1);
-    a0 = fmaf(row_ror<10>(v), w[10], a0); a1 = fmaf(row_ror<11>(v), w[11], a1);
-    a0 = fmaf(row_ror<12>(v), w[12], a0); a1 = fmaf(row_ror<13>(v), w[13], a1);
-    a0 = fmaf(row_ror<14>(v), w[14], a0); a1 = fmaf(row_ror<15>(v), w[15], a1);
+    float a0, a1;
+    asm volatile(
+        "s_nop 1\n"
+        "v_mul_f32_e32 %0, %2, %3\n"
+        "v_mul_f32_dpp %1, %2, %4" DEER_RR(1)
+        "v_fmac_f32_dpp %0, %2, %5" DEER_RR(2)
+        "v_fmac_f32_dpp %1, %2, %6" DEER_RR(3)
+        "v_fmac_f32_dpp %0, %2, %7" DEER_RR(4)
+        "v_fmac_f32_dpp %1, %2, %8" DEER_RR(5)
+        "v_fmac_f32_dpp %0, %2, %9" DEER_RR(6)
+        "v_fmac_f32_dpp %1, %2, %10" DEER_RR(7)
+        "v_fmac_f32_dpp %0, %2, %11" DEER_RR(8)
+        "v_fmac_f32_dpp %1, %2, %12" DEER_RR(9)
+        "v_fmac_f32_dpp %0, %2, %13" DEER_RR(10)
+        "v_fmac_f32_dpp %1, %2, %14" DEER_RR(11)
+        "v_fmac_f32_dpp %0, %2, %15" DEER_RR(12)
+        "v_fmac_f32_dpp %1, %2, %16" DEER_RR(13)
+        "v_fmac_f32_dpp %0, %2, %17" DEER_RR(14)
+        "v_fmac_f32_dpp %1, %2, %18" DEER_RR(15)
+        : "=&v"(a0), "=&v"(a1)
+        : "v"(v), "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "v"(w[4]), "v"(w[5]), "v"(w[6]), "v"(w[7]), "v"(w[8]),
+          "v"(w[9]), "v"(w[10]), "v"(w[11]), "v"(w[12]), "v"(w[13]), "v"(w[14]), "v"(w[15]));
     return a0 + a1;
 }
+#undef DEER_RR
 
 // Buffer resource with a wave-uniform base: an access adds a per-lane byte offset (VGPR) and a
 // wave-uniform byte offset (SGPR).  A lane offset of 2^31 or more is outside the resource: a
@@ -631,17 +644,19 @@ __device__ __forceinline__ void damp_tile(v4f (&acc)[4], const Chains16 &w, int 
     }
 }
 
-// one matrix-core step of chain n: acc <- (diag(d) + W diag(m)) acc (layout of the MP = 16
-// generic kernel: Aop = columns of W p, dI = rows of diag(A) p)
-__device__ __forceinline__ void mfma_step16(v4f &acc, uint32_t wn, int g, const float (&Aop)[4],
-                                            const float (&dI)[4]) {
-    float Bop[4];
+// one matrix-core step of chain n: acc <- (diag(d) + W p diag(m)) acc.  The mask and the
+// diagonal go into the A operand: lane (g, c) supplies, for k = 4 g + q, m_k ? WpD[q] : Dq[q]
+// with WpD = (W p)[c][k] + [c == k] d_k and Dq = [c == k] d_k, so B is the product unchanged.
+__device__ __forceinline__ v4f mfma_step16(const v4f &acc, uint32_t wn, int g, const float (&WpD)[4],
+                                           const float (&Dq)[4]) {
+    v4f nx = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int q = 0; q < 4; ++q) Bop[q] = select_bit(wn, 4 * g + q, acc[q]);
-#pragma unroll
-    for (int r2 = 0; r2 < 4; ++r2) acc[r2] *= dI[r2];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) acc = mfma16x16x4(Aop[q], Bop[q], acc);
+    for (int q = 0; q < 4; ++q) {
+        const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)wn, 4 * g + q, 1);
+        const float a = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+        nx = mfma16x16x4(a, acc[q], nx);
+    }
+    return nx;
 }
 
 template <int TB>
@@ -650,18 +665,19 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
     const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
     const int *__restrict__ zsel, float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout,
     float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
-    int ncs) {
+    int ncs, int wmaps) {
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int nchains = B * ncs;
     const int chain0 = blockIdx.x * 4;
     const Chains16 w = chains16(chain0, nchains, ncs, C, T, active, gamma, zsel);
     if (w.maxlen == 0) return;
-    float Aop[4], dI[4];
+    float WpD[4], Dq[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int col = 4 * g + q;
-        Aop[q] = (c < M && col < M) ? W[c * M + col] * p_of(col, N, alpha) : 0.f;
-        dI[q] = col < M ? A[col] * p_of(col, N, alpha) : 0.f;
+        const float wp = (c < M && col < M) ? W[c * M + col] * p_of(col, N, alpha) : 0.f;
+        Dq[q] = (col == c && col < M) ? A[col] * p_of(col, N, alpha) : 0.f;
+        WpD[q] = wp + Dq[q];
     }
     v4f acc[4];
 #pragma unroll
@@ -736,19 +752,23 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
                 const bool pos = (posb >> tt) & 1u;
                 const uint64_t bal = __ballot(pos);
                 // the four chains' updates interleaved: k-slice outer, chain inner
-                float Bop[4][4];
+                float Am[4][4];
 #pragma unroll
                 for (int n = 0; n < 4; ++n)
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) Bop[n][q] = select_bit((uint32_t)(bal >> (16 * n)), 4 * g + q, acc[n][q]);
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
+                        Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+                    }
+                v4f nx[4];
 #pragma unroll
-                for (int n = 0; n < 4; ++n)
-#pragma unroll
-                    for (int r2 = 0; r2 < 4; ++r2) acc[n][r2] *= dI[r2];
+                for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
 #pragma unroll
-                    for (int n = 0; n < 4; ++n) acc[n] = mfma16x16x4(Aop[q], Bop[n][q], acc[n]);
+                    for (int n = 0; n < 4; ++n) nx[n] = mfma16x16x4(Am[n][q], acc[n][q], nx[n]);
+#pragma unroll
+                for (int n = 0; n < 4; ++n) acc[n] = nx[n];
                 const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
                 u = fmaf(ugam, y, -zv[tt]);
             }
@@ -774,7 +794,7 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
                 }
 #pragma unroll
                 for (int n = 0; n < 4; ++n)
-                    if (t < w.plen[n]) mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, Aop, dI);
+                    if (t < w.plen[n]) acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
                 const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
                 if (run) {
                     u = fmaf(ugam, y, -r);
@@ -783,6 +803,58 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
             }
         }
         damp_tile(acc, w, t0, tl);
+    }
+    if (wmaps) {
+        // The wave's four chunks (one sequence, all active) composed for the carry pass:
+        //   slot chain0:      wave map  Q = P_3 P_2 P_1 P_0,  u_w = the four chunks' walk from 0
+        //   slot chain0 + n:  prefix    R_n = P_{n-1} ... P_0, s_n = the walk of the first n chunks
+        // so that carry(chain0 + n) = R_n carry(chain0) + s_n.  A chunk product in accumulator
+        // layout is transposed through LDS into the A-operand layout; vectors ride in column 0.
+        __shared__ float lt[4][16][17];
+        __shared__ float lv[4][16];
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) lt[n][4 * g + r2][c] = acc[n][r2];
+        lv[g][c] = u;
+        lds_barrier();
+        float Am[3][4];
+        v4f bv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+#pragma unroll
+            for (int n = 1; n < 4; ++n) Am[n - 1][q] = lt[n][c][4 * g + q];
+#pragma unroll
+            for (int n = 0; n < 4; ++n) bv[n][q] = c == 0 ? lv[n][4 * g + q] : 0.f;
+        }
+        v4f R2 = {0.f, 0.f, 0.f, 0.f}, R3 = {0.f, 0.f, 0.f, 0.f}, Qw = {0.f, 0.f, 0.f, 0.f};
+        v4f s2 = bv[1], s3 = bv[2], uw = bv[3];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            R2 = mfma16x16x4(Am[0][q], acc[0][q], R2);
+            s2 = mfma16x16x4(Am[0][q], bv[0][q], s2);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            R3 = mfma16x16x4(Am[1][q], R2[q], R3);
+            s3 = mfma16x16x4(Am[1][q], s2[q], s3);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            Qw = mfma16x16x4(Am[2][q], R3[q], Qw);
+            uw = mfma16x16x4(Am[2][q], s3[q], uw);
+        }
+        const v4f outm[4] = {Qw, acc[0], R2, R3}, outv[4] = {uw, bv[0], s2, s3};
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+            float *P = Pout + (size_t)(chain0 + n) * 256;
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) P[(4 * g + r2) * 16 + c] = outm[n][r2];
+            if (c == 0)
+                *reinterpret_cast<float4 *>(vout + (size_t)(chain0 + n) * 16 + 4 * g) =
+                    make_float4(outv[n][0], outv[n][1], outv[n][2], outv[n][3]);
+        }
+        return;
     }
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
@@ -796,6 +868,57 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
     if (okc) vout[(size_t)id * 16 + c] = u;
 }
 
+// Convergence test and update safeguard of one pass for sequence b from its maxima e = max
+// |Delta| bits and zm = max |z| bits: accept the update (flip sel, count it, relax the damping,
+// freeze the sequence once max|Delta| < tol), or reject it (keep sel, raise the damping:
+// 1 - gamma = first, then x grow up to 1 = the fixed-point step); a non-finite fixed-point step
+// ends the sequence.
+__device__ __forceinline__ void seq_decide(int b, uint32_t e, uint32_t zm, const NewtonDev &nd, float tol, float bound,
+                                           const NewtonDamp &dp) {
+    const float ef = __uint_as_float(e), zf = __uint_as_float(zm);
+    const bool fin = e < 0x7f800000u;
+    float om = nd.om[b];
+    const bool keep = fin && (bound < 0.f || om >= 1.f || ef <= bound * (1.f + zf));
+    if (keep) {
+        nd.sel[b] ^= 1;
+        nd.it[b] += 1;
+        nd.norm[b] = ef;
+        if (om > 0.f) om = om / dp.shrink < dp.floor ? 0.f : om / dp.shrink;
+        if (ef < tol) {
+            nd.act[b] = 0;
+            nd.status[b] = 1;
+        }
+    } else if (om >= 1.f) {
+        nd.norm[b] = ef;
+        nd.act[b] = 0;
+        nd.status[b] = 2;
+    } else {
+        om = om == 0.f ? dp.first : fminf(1.f, om * dp.grow);
+    }
+    nd.om[b] = om;
+    nd.gamma[b] = 1.f - om;
+}
+
+// Arrival of `cnt` chains of sequence b with maxima e, zm (see FusedCtl).  Device-scope atomics
+// meet at one coherence point across the XCDs; each maximum is returned (so performed) before
+// the count is raised, so the chain that completes the count reads the final maxima.
+__device__ __forceinline__ void seq_arrive(const FusedCtl &fc, int b, int cnt, int ncs, uint32_t e, uint32_t zm) {
+    uint32_t *blk = fc.seq + (size_t)b * kSeqWords;   // count | max |Delta| | max |z|, 128 bytes apart
+    const uint32_t r1 = __hip_atomic_fetch_max(blk + 32, e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t r2 = __hip_atomic_fetch_max(blk + 64, zm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // the count may only move once both maxima are in: the increment depends on their return
+    // values (|x| bits are below 2^31, so the added term is zero)
+    const uint32_t old = __hip_atomic_fetch_add(blk, (uint32_t)cnt + ((r1 | r2) >> 31), __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+    if (old + (uint32_t)cnt != (uint32_t)ncs) return;
+    const uint32_t ef = __hip_atomic_load(blk + 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t zf = __hip_atomic_load(blk + 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    seq_decide(b, ef, zf, fc.nd, fc.tol, fc.bound, fc.dp);
+    __hip_atomic_store(blk + 32, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(blk + 64, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(blk, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 template <int TB>
 __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restrict__ A, const float *__restrict__ W,
                                                           float alpha, int N, const uint32_t *__restrict__ masks,
@@ -804,7 +927,8 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
                                                           uint32_t *__restrict__ chain_bits,
                                                           const int *__restrict__ active,
                                                           const float *__restrict__ gamma, int B, int T, int M, int C,
-                                                          int ncs) {
+                                                          int ncs, const float *__restrict__ Pm,
+                                                          const float *__restrict__ vmap, FusedCtl fc) {
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int nchains = B * ncs;
     const int chain0 = blockIdx.x * 4;
@@ -828,11 +952,30 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
 #pragma unroll
     for (int k = 0; k < 16; ++k) wp[k] = (lat && src[k] < M) ? W[c * M + src[k]] * p_of(src[k], N, alpha) : 0.f;
     const float d = lat ? A[c] * p_of(c, N, alpha) : 0.f;
-    float D = (len > 0 && lat) ? carry_in[(size_t)id * 16 + c] : 0.f;
+    float D = 0.f;
+    if (len > 0 && lat) {
+        if (!Pm || g == 0) {
+            D = carry_in[(size_t)id * 16 + c];
+        } else {   // composed wave maps: carry = R_g carry(chain0) + s_g
+            const float4 *R4 = reinterpret_cast<const float4 *>(Pm + (size_t)id * 256 + c * 16);
+            const float4 *w4 = reinterpret_cast<const float4 *>(carry_in + (size_t)chain0 * 16);
+            float a0 = vmap[(size_t)id * 16 + c], a1 = 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 rr4 = R4[q], ww = w4[q];
+                a0 = fmaf(rr4.x, ww.x, a0);
+                a1 = fmaf(rr4.y, ww.y, a1);
+                a0 = fmaf(rr4.z, ww.z, a0);
+                a1 = fmaf(rr4.w, ww.w, a1);
+            }
+            D = a0 + a1;
+        }
+    }
     const float *zin = cur_iter(zbuf, zalt, zsel, b);
     float *zout = next_iter(zbuf, zalt, zsel, b);
-    const int b0 = chain0 / ncs;
-    const size_t row0 = (size_t)b0 * T + (size_t)(chain0 % ncs) * C;
+    const int cl0 = min(chain0, nchains - 1);   // a wave past the last chain touches no memory
+    const int b0 = cl0 / ncs;
+    const size_t row0 = (size_t)b0 * T + (size_t)(cl0 % ncs) * C;
     const uint32_t drow = (uint32_t)((size_t)b * T + s0 - row0);
     const auto rr = wave_rsrc(r + row0 * M), rm = wave_rsrc(masks + row0);
     const auto rzi = wave_rsrc(cur_iter(zbuf, zalt, zsel, b0) + row0 * M);
@@ -891,9 +1034,37 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
         emax = emax > o ? emax : o;
         zmax = zmax > oz ? zmax : oz;
     }
-    if (len > 0 && c == 0) {   // per-chain maxima, reduced per sequence by k_seq_max / k_seq_ctl
-        chain_bits[id] = emax;
-        chain_bits[(size_t)nchains + id] = zmax;
+    if (!fc.seq) {
+        if (len > 0 && c == 0) {   // per-chain maxima, reduced per sequence by k_seq_max / k_seq_ctl
+            chain_bits[id] = emax;
+            chain_bits[(size_t)nchains + id] = zmax;
+        }
+        return;
+    }
+    // fused pass-end control: lane 0 gathers the four chains' maxima and arrives once per
+    // sequence they belong to
+    uint32_t em[4], zm[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        em[n] = (uint32_t)__shfl((int)emax, 16 * n, 64);
+        zm[n] = (uint32_t)__shfl((int)zmax, 16 * n, 64);
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+            const int bn = (chain0 + n) / ncs;
+            if (w.plen[n] == 0 || (n > 0 && w.plen[n - 1] > 0 && (chain0 + n - 1) / ncs == bn)) continue;
+            uint32_t E = 0u, Z = 0u;
+            int cnt = 0;
+#pragma unroll
+            for (int m = n; m < 4; ++m)
+                if (w.plen[m] > 0 && (chain0 + m) / ncs == bn) {
+                    E = E > em[m] ? E : em[m];
+                    Z = Z > zm[m] ? Z : zm[m];
+                    ++cnt;
+                }
+            seq_arrive(fc, bn, cnt, ncs, E, Z);
+        }
     }
 }
 
@@ -1313,6 +1484,104 @@ __global__ __launch_bounds__(64) void k_carry_group16(const float *__restrict__ 
         *reinterpret_cast<float4 *>(gu + ((size_t)b * ngroups + j) * 16 + 4 * g) = make_float4(u[0], u[1], u[2], u[3]);
 }
 
+// Carries of composed wave maps (four chunks each, at chunk slots 4w): one block per sequence,
+// NWV waves.  Each wave composes a contiguous range of maps into one, wave 0 walks the NWV
+// composed maps (LDS), and every wave walks its range again from its own carry, writing the
+// carry of each wave map into the carry slot of its first chunk.
+constexpr int WALK_NWV = 16;
+__global__ __launch_bounds__(WALK_NWV * 64) void k_carry_walk16(const float *__restrict__ P, const float *__restrict__ v,
+                                                               float *__restrict__ carry,
+                                                               const int *__restrict__ active, int ncs) {
+    constexpr int PF = 8;
+    __shared__ float ls[WALK_NWV][16][17];
+    __shared__ float lt[WALK_NWV][16], lsc[WALK_NWV][16];
+    const int b = blockIdx.x;
+    if (active && !active[b]) return;
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+    const int nw = ncs >> 2, per = (nw + WALK_NWV - 1) / WALK_NWV;
+    const int w0 = min(wv * per, nw), w1 = min(w0 + per, nw);
+    const float *Pb = P + (size_t)b * ncs * 256, *vb = v + (size_t)b * ncs * 16;
+    auto fetch = [&](int wm, float (&a)[4], float (&vv)[4]) {
+        carry16_fetch<false>(Pb + (size_t)(4 * wm) * 256, vb + (size_t)(4 * wm) * 16, g, c, a, vv);
+    };
+    float a[PF][4], vv[PF][4];
+    // composed map of this wave's range
+    v4f S, t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) S[r] = (4 * g + r == c) ? 1.f : 0.f;
+    if (w0 < w1) {
+#pragma unroll
+        for (int d = 0; d < PF; ++d) fetch(min(w0 + d, w1 - 1), a[d], vv[d]);
+        for (int k = w0; k < w1; k += PF) {
+#pragma unroll
+            for (int d = 0; d < PF; ++d) {
+                if (k + d >= w1) break;
+                v4f ns = {0.f, 0.f, 0.f, 0.f}, nt = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    ns = mfma16x16x4(a[d][q], S[q], ns);
+                    nt = mfma16x16x4(a[d][q], t[q], nt);
+                }
+                if (c == 0) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) nt[r] += vv[d][r];
+                }
+                S = ns;
+                t = nt;
+                fetch(min(k + d + PF, w1 - 1), a[d], vv[d]);
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) ls[wv][4 * g + r][c] = S[r];
+    if (c == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) lt[wv][4 * g + r] = t[r];
+    }
+    __syncthreads();
+    if (wv == 0) {   // walk of the composed maps
+        v4f cur = {0.f, 0.f, 0.f, 0.f};
+        for (int k = 0; k < WALK_NWV; ++k) {
+            if (c == 0) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) lsc[k][4 * g + r] = cur[r];
+            }
+            v4f nx;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) nx[r] = c == 0 ? lt[k][4 * g + r] : 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) nx = mfma16x16x4(ls[k][c][4 * g + q], cur[q], nx);
+            cur = nx;
+        }
+    }
+    __syncthreads();
+    if (w0 >= w1) return;
+    v4f cur;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) cur[r] = c == 0 ? lsc[wv][4 * g + r] : 0.f;
+#pragma unroll
+    for (int d = 0; d < PF; ++d) fetch(min(w0 + d, w1 - 1), a[d], vv[d]);
+    for (int k = w0; k < w1; k += PF) {
+#pragma unroll
+        for (int d = 0; d < PF; ++d) {
+            const int wm = k + d;
+            if (wm >= w1) break;
+            if (c == 0)
+                *reinterpret_cast<float4 *>(carry + ((size_t)b * ncs + 4 * wm) * 16 + 4 * g) =
+                    make_float4(cur[0], cur[1], cur[2], cur[3]);
+            v4f nx = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) nx = mfma16x16x4(a[d][q], cur[q], nx);
+            if (c == 0) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) nx[r] += vv[d][r];
+            }
+            cur = nx;
+            fetch(min(wm + PF, w1 - 1), a[d], vv[d]);
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------------------
 // forward fix-up: Delta from the carry, z += Delta, per-sequence max |Delta|
 // ---------------------------------------------------------------------------------------
@@ -1460,28 +1729,7 @@ __global__ __launch_bounds__(256) void k_seq_ctl(const uint32_t *__restrict__ ch
         e = e > red[0][w] ? e : red[0][w];
         zm = zm > red[1][w] ? zm : red[1][w];
     }
-    const float ef = __uint_as_float(e), zf = __uint_as_float(zm);
-    const bool fin = e < 0x7f800000u;
-    float om = nd.om[b];
-    const bool keep = fin && (bound < 0.f || om >= 1.f || ef <= bound * (1.f + zf));
-    if (keep) {
-        nd.sel[b] ^= 1;
-        nd.it[b] += 1;
-        nd.norm[b] = ef;
-        if (om > 0.f) om = om / dp.shrink < dp.floor ? 0.f : om / dp.shrink;
-        if (ef < tol) {
-            nd.act[b] = 0;
-            nd.status[b] = 1;
-        }
-    } else if (om >= 1.f) {
-        nd.norm[b] = ef;
-        nd.act[b] = 0;
-        nd.status[b] = 2;
-    } else {
-        om = om == 0.f ? dp.first : fminf(1.f, om * dp.grow);
-    }
-    nd.om[b] = om;
-    nd.gamma[b] = 1.f - om;
+    seq_decide(b, e, zm, nd, tol, bound, dp);
 }
 
 int launch_seq_ctl(const uint32_t *chain_bits, const NewtonDev &nd, int B, int ncs, float tol, float bound,
@@ -1492,9 +1740,13 @@ int launch_seq_ctl(const uint32_t *chain_bits, const NewtonDev &nd, int B, int n
     return DEER_OK;
 }
 
-__global__ void k_ctl_init(NewtonDev nd, int B) {
+__global__ void k_ctl_init(NewtonDev nd, uint32_t *seq, int B) {
     const int b = blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= B) return;
+    if (seq) {
+#pragma unroll
+        for (int k = 0; k < 3; ++k) seq[(size_t)b * kSeqWords + 32 * k] = 0u;
+    }
     nd.act[b] = 1;
     nd.gamma[b] = 1.f;
     nd.sel[b] = 0;
@@ -1504,8 +1756,8 @@ __global__ void k_ctl_init(NewtonDev nd, int B) {
     nd.status[b] = 0;
 }
 
-int launch_ctl_init(const NewtonDev &nd, int B, hipStream_t st) {
-    hipLaunchKernelGGL(k_ctl_init, dim3((B + 255) / 256), dim3(256), 0, st, nd, B);
+int launch_ctl_init(const NewtonDev &nd, uint32_t *seq, int B, hipStream_t st) {
+    hipLaunchKernelGGL(k_ctl_init, dim3((B + 255) / 256), dim3(256), 0, st, nd, seq, B);
     DEER_LAUNCH_CHECK("k_ctl_init");
     return DEER_OK;
 }
@@ -1654,6 +1906,11 @@ size_t reduce_gpart_ws_bytes(int MP) { return (size_t)GP_SLICES * MP * (MP + 2) 
 // ---------------------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------------------
+static int invalid_arg(const char *what) {
+    set_error("%s", what);
+    return DEER_ERR_INVALID_ARG;
+}
+
 static int padded(int M) { return M <= 16 ? 16 : (M <= 32 ? 32 : 64); }
 
 int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, float *J, uint32_t *masks,
@@ -1698,7 +1955,7 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
 
 int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
                                 uint32_t *masks, float *P, float *v, const int *active, const float *gamma, int C,
-                                int ncs, hipStream_t st) {
+                                int ncs, bool wmaps, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
@@ -1706,16 +1963,20 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
 #define NP(MPV)                                                                                                   \
     hipLaunchKernelGGL(k_newton_product_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, \
                        a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs)
+    if (wmaps && (MP != 16 || ncs % 4))
+        return invalid_arg("composed wave maps need M <= 16 and a chunk count divisible by 4");
     if (MP == 64 && (a.N == 0 || a.N == a.M)) {   // uniform forcing factor: W-in-LDS kernel
         hipLaunchKernelGGL(k_newton_product_plrnn64u, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0,
                            z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
     } else if (MP == 16) {
         if (C <= 16)
             hipLaunchKernelGGL(k_newton_product_plrnn16<16>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
-                               a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
+                               a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs,
+                               (int)wmaps);
         else
             hipLaunchKernelGGL(k_newton_product_plrnn16<32>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
-                               a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
+                               a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs,
+                               (int)wmaps);
     } else if (MP == 32) NP(32); else NP(64);
 #undef NP
     DEER_LAUNCH_CHECK("k_newton_product_plrnn");
@@ -1790,9 +2051,19 @@ int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_
     return DEER_OK;
 }
 
+int launch_carry_walk16(const float *P, const float *v, float *carry, const int *active, int B, int ncs,
+                        hipStream_t st) {
+    if (ncs % 4) return invalid_arg("wave-map walk needs a chunk count divisible by 4");
+    KTimer kt("k_carry", st);
+    hipLaunchKernelGGL(k_carry_walk16, dim3(B), dim3(WALK_NWV * 64), 0, st, P, v, carry, active, ncs);
+    DEER_LAUNCH_CHECK("k_carry_walk16");
+    return DEER_OK;
+}
+
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
                            float *z, float *zalt, const int *zsel, uint32_t *chain_bits, const int *active,
-                           const float *gamma, int C, int ncs, hipStream_t st) {
+                           const float *gamma, int C, int ncs, const float *Pm, const float *vm,
+                           const FusedCtl *fc, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
@@ -1802,7 +2073,12 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
                        z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
 #define FX16(TBV)                                                                                              \
     hipLaunchKernelGGL(k_fixup_fwd_plrnn16<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, \
-                       carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
+                       carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs, Pm, vm, fcv)
+    if (Pm && (MP != 16 || ncs % 4))
+        return invalid_arg("composed wave maps need M <= 16 and a chunk count divisible by 4");
+    if (fc && MP != 16) return invalid_arg("the fused pass-end control needs M <= 16");
+    FusedCtl fcv{};
+    if (fc) fcv = *fc;
     if (MP == 16) {
         if (C <= 16) FX16(16); else FX16(32);
     } else if (MP == 32) FX(32); else FX(64);

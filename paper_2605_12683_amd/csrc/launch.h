@@ -4,6 +4,8 @@
 
 namespace deer {
 
+struct FusedCtl;   // pass-end control fused into the M <= 16 fix-up (defined below)
+
 struct PlrnnArgs {
     const float *A, *W, *h;
     float alpha;
@@ -30,13 +32,18 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
                                hipStream_t st);
 int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
                                 uint32_t *masks, float *P, float *v, const int *active, const float *gamma, int C,
-                                int ncs, hipStream_t st);
+                                int ncs, bool wmaps, hipStream_t st);
+// M <= 16 with wave maps (P, v from launch_newton_product_plrnn with wmaps): carries of the
+// wave maps, written to the carry slot of each wave's first chunk
+int launch_carry_walk16(const float *P, const float *v, float *carry, const int *active, int B, int ncs,
+                        hipStream_t st);
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
                  uint32_t *norm_bits, int B, int ncs, float *gws, hipStream_t st);
 size_t carry_ws_floats(int MP, int B, int ncs);
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
                            float *z, float *zalt, const int *zsel, uint32_t *chain_bits, const int *active,
-                           const float *gamma, int C, int ncs, hipStream_t st);
+                           const float *gamma, int C, int ncs, const float *Pm, const float *vm,
+                           const FusedCtl *fc, hipStream_t st);
 // device-side Newton control (one entry per sequence)
 struct NewtonDev {
     int *act;       // active flag (read by every kernel of a pass)
@@ -52,7 +59,17 @@ struct NewtonDamp {
 };
 int launch_seq_ctl(const uint32_t *chain_bits, const NewtonDev &nd, int B, int ncs, float tol, float bound,
                    const NewtonDamp &dp, hipStream_t st);
-int launch_ctl_init(const NewtonDev &nd, int B, hipStream_t st);
+// The pass-end control of k_seq_ctl taken by the fix-up itself: per sequence a 96-word block of
+// seq (arrival count, max |Delta| bits, max |z| bits, one 128-byte line each) is updated with device-scope atomics and the
+// last chain of the sequence to arrive takes the decision.  seq == nullptr: not fused.
+struct FusedCtl {
+    NewtonDev nd;
+    uint32_t *seq;
+    float tol, bound;
+    NewtonDamp dp;
+};
+constexpr int kSeqWords = 96;
+int launch_ctl_init(const NewtonDev &nd, uint32_t *seq, int B, hipStream_t st);
 int launch_seq_max(const uint32_t *chain_bits, const int *active, uint32_t *norm_bits, int B, int ncs,
                    hipStream_t st);
 int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *g, float seed_scale, const float *z,

@@ -446,7 +446,7 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
         const bool wm = w.MP == 16 && w.ncs % 4 == 0;
         if ((r = launch_newton_product_plrnn(a, zb, za, zsel, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, wm, st)))
             return r;
-        if (wm) r = launch_carry_walk16(w.P, w.v, w.carry, dact, B, w.ncs, st);
+        if (wm) r = launch_carry_walk16(false, w.P, w.v, w.carry, dact, B, w.ncs, st);
         else r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, nullptr, B, w.ncs, w.gws, st);
         if (r) return r;
         return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, zb, za, zsel, w.ctl.chain_bits, dact, gam, w.C, w.ncs,
@@ -655,6 +655,16 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
         PlrnnWs w = carve_plrnn(ws, B, T, m->M, DEER_OP_ADJOINT, &need);
         PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
         const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
+        if (w.MP == 16) {   // register-tiled path: masks from z inside the kernels, per-wave gradients
+            if ((rc = launch_adjoint_plrnn16(a, g, scale, z, w.P, w.v, w.carry, lam, w.gpart, w.C, w.ncs, st)))
+                return rc;
+            if (grads && (grads->A || grads->W || grads->h)) {
+                if ((rc = launch_reduce_gpart(w.gpart, (B * w.ncs + 3) / 4, 16, m->M, grads->A, grads->W, grads->h,
+                                              w.gpart2, st)))
+                    return rc;
+            }
+            return DEER_OK;
+        }
         if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, w.masks, nullptr, st))) return rc;
         if ((rc = launch_chunk_product_plrnn(a, true, w.masks, g, z, scale, w.P, w.v, nullptr, w.C, w.ncs, st)))
             return rc;

@@ -1484,11 +1484,423 @@ __global__ __launch_bounds__(64) void k_carry_group16(const float *__restrict__ 
         *reinterpret_cast<float4 *>(gu + ((size_t)b * ngroups + j) * 16 + 4 * g) = make_float4(u[0], u[1], u[2], u[3]);
 }
 
-// Carries of composed wave maps (four chunks each, at chunk slots 4w): one block per sequence,
-// NWV waves.  Each wave composes a contiguous range of maps into one, wave 0 walks the NWV
-// composed maps (LDS), and every wave walks its range again from its own carry, writing the
-// carry of each wave map into the carry slot of its first chunk.
+// d[k] += v(row_src(lane, k)) * s for k = 0..15: the rank-one update of a rotated row, e.g.
+// dW[i][row_src(i, k)] += lam_i relu(z~)_{row_src(i, k)}.  All 64 lanes must be active.
+#define DEER_RR(k) " row_ror:" #k " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+__device__ __forceinline__ void row16_outer(float (&d)[16], float v, float s) {
+    asm volatile(
+        "s_nop 1\n"
+        "v_fmac_f32_e32 %0, %16, %17\n"
+        "v_fmac_f32_dpp %1, %16, %17" DEER_RR(1)
+        "v_fmac_f32_dpp %2, %16, %17" DEER_RR(2)
+        "v_fmac_f32_dpp %3, %16, %17" DEER_RR(3)
+        "v_fmac_f32_dpp %4, %16, %17" DEER_RR(4)
+        "v_fmac_f32_dpp %5, %16, %17" DEER_RR(5)
+        "v_fmac_f32_dpp %6, %16, %17" DEER_RR(6)
+        "v_fmac_f32_dpp %7, %16, %17" DEER_RR(7)
+        "v_fmac_f32_dpp %8, %16, %17" DEER_RR(8)
+        "v_fmac_f32_dpp %9, %16, %17" DEER_RR(9)
+        "v_fmac_f32_dpp %10, %16, %17" DEER_RR(10)
+        "v_fmac_f32_dpp %11, %16, %17" DEER_RR(11)
+        "v_fmac_f32_dpp %12, %16, %17" DEER_RR(12)
+        "v_fmac_f32_dpp %13, %16, %17" DEER_RR(13)
+        "v_fmac_f32_dpp %14, %16, %17" DEER_RR(14)
+        "v_fmac_f32_dpp %15, %16, %17" DEER_RR(15)
+        : "+v"(d[0]), "+v"(d[1]), "+v"(d[2]), "+v"(d[3]), "+v"(d[4]), "+v"(d[5]), "+v"(d[6]), "+v"(d[7]), "+v"(d[8]),
+          "+v"(d[9]), "+v"(d[10]), "+v"(d[11]), "+v"(d[12]), "+v"(d[13]), "+v"(d[14]), "+v"(d[15])
+        : "v"(v), "v"(s));
+}
+#undef DEER_RR
+
+// ---------------------------------------------------------------------------------------
+// M <= 16 reverse (adjoint) pass, per chunk [s0, s1) (gradients appendix):
+//   P_c = J~_{s1} ... J~_{s0+1} over the steps below T (the carry pass takes its transpose)
+//   v_c = lam_{s0} from lam_{s1} = 0,   lam_k = J~_{k+1}^T lam_{k+1} + g_k
+// The masks m_s = [z~_s > 0] are formed here from z and x.  A tile row tt is chunk row
+// t0 + tt: z_{s0+t0+tt}, x_{s0+t0+tt+1} (so z~ of step s0+t0+tt+1, the mask lam_k needs) and
+// g_{s0+t0+tt}.  The products run forward over the tiles, the local adjoint backward.
+// ---------------------------------------------------------------------------------------
+template <int TB>
+__global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
+    const float *__restrict__ A, const float *__restrict__ W, float alpha, int N, const float *__restrict__ rhs,
+    const float *__restrict__ z, const float *__restrict__ x, float seed_scale, float *__restrict__ Pout,
+    float *__restrict__ vout, int B, int T, int M, int C, int ncs, int wmaps) {
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int nchains = B * ncs;
+    const int chain0 = blockIdx.x * 4;
+    const Chains16 w = chains16(chain0, nchains, ncs, C, T, nullptr, nullptr, nullptr);
+    if (w.maxlen == 0) return;
+    int pl[4];   // product steps: a chunk that ends at T has one fewer
+    int minP = C;
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        const int s1 = ((chain0 + n) % ncs) * C + w.plen[n];
+        pl[n] = w.plen[n] - ((w.plen[n] > 0 && s1 == T) ? 1 : 0);
+        minP = min(minP, pl[n]);
+    }
+    float WpD[4], Dq[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int col = 4 * g + q;
+        const float wp = (c < M && col < M) ? W[c * M + col] * p_of(col, N, alpha) : 0.f;
+        Dq[q] = (col == c && col < M) ? A[col] * p_of(col, N, alpha) : 0.f;
+        WpD[q] = wp + Dq[q];
+    }
+    v4f acc[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[n][r] = (4 * g + r == c) ? 1.f : 0.f;
+    const int id = chain0 + g;
+    const bool okc = id < nchains;
+    const int b = okc ? id / ncs : 0, s0 = okc ? (id % ncs) * C : 0;
+    int len = 0;
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+        if (n == g) len = w.plen[n];
+    const bool lat = c < M, forced = c < N;
+    int src[16];
+    row_sources(c, src);
+    float wT[16];   // rotated row c of W^T
+#pragma unroll
+    for (int k = 0; k < 16; ++k) wT[k] = (lat && src[k] < M) ? W[src[k] * M + c] : 0.f;
+    const float pi = p_of(c, N, alpha), Ai = lat ? A[c] : 0.f;
+    const int b0 = chain0 / ncs, s00 = (chain0 % ncs) * C;
+    const size_t row0 = (size_t)b0 * T + s00, xrow0 = (size_t)b0 * (T + 1) + s00 + 1;
+    const uint32_t drow = (uint32_t)((size_t)b * T + s0 - row0);
+    const uint32_t dxrow = (uint32_t)((size_t)b * (T + 1) + s0 + 1 - xrow0);
+    const auto rz = wave_rsrc(z + row0 * M), rg = wave_rsrc(rhs ? rhs + row0 * M : z);
+    const auto rx = wave_rsrc(N > 0 ? x + xrow0 * N : z);
+    const uint32_t vz = lat ? 4u * (drow * M + c) : kOffLane;
+    const uint32_t vx = forced ? 4u * (dxrow * N + c) : kOffLane;
+    const uint32_t vg = (rhs && lat) ? vz : kOffLane;
+    float zv[TB], xv[TB];
+    uint32_t posb = 0u;
+    int loaded = -1;   // t0 of the tile whose rows zv/xv hold
+    auto load_tile = [&](int t0) {
+#pragma unroll
+        for (int tt = 0; tt < TB; ++tt) {
+            zv[tt] = bload(rz, vz, 4 * (t0 + tt) * M);
+            xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
+        }
+        posb = 0u;
+#pragma unroll
+        for (int tt = 0; tt < TB; ++tt) {
+            const float zt = forced ? __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt])) : zv[tt];
+            posb |= (zt > 0.f ? 1u : 0u) << tt;
+        }
+        loaded = t0;
+    };
+    // z~ of step s = s0 + t + 1 for the slow path (chunk row t)
+    auto ztilde_next = [&](int t) {
+        if (!(t < len && lat)) return 0.f;
+        const int s = s0 + t + 1;
+        const float zp = z[((size_t)b * T + s - 1) * M + c];
+        if (!forced) return zp;
+        return __fadd_rn(__fmul_rn(pi, zp), __fmul_rn(alpha, x[((size_t)b * (T + 1) + s) * N + c]));
+    };
+    // ---- chunk products, forward over the tiles
+    for (int t0 = 0; t0 < w.maxlen; t0 += TB) {
+        const int tl = min(TB, w.maxlen - t0);
+        if (t0 + TB <= w.minlen) {
+            load_tile(t0);
+            if (t0 + TB <= minP) {
+#pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    const uint64_t bal = __ballot((posb >> tt) & 1u);
+                    float Am[4][4];
+#pragma unroll
+                    for (int n = 0; n < 4; ++n)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t m =
+                                (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
+                            Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+                        }
+                    v4f nx[4];
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+#pragma unroll
+                        for (int n = 0; n < 4; ++n) nx[n] = mfma16x16x4(Am[n][q], acc[n][q], nx[n]);
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) acc[n] = nx[n];
+                }
+            } else {
+#pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    const uint64_t bal = __ballot((posb >> tt) & 1u);
+#pragma unroll
+                    for (int n = 0; n < 4; ++n)
+                        if (t0 + tt < pl[n]) acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
+                }
+            }
+        } else {
+            for (int t = t0; t < t0 + tl; ++t) {
+                const uint64_t bal = __ballot(ztilde_next(t) > 0.f);
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+                    if (t < pl[n]) acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
+            }
+        }
+    }
+    // ---- local adjoint from a zero carry, backward over the tiles
+    float u = 0.f;
+    const int last = ((w.maxlen - 1) / TB) * TB;
+    for (int t0 = last; t0 >= 0; t0 -= TB) {
+        const int tl = min(TB, w.maxlen - t0);
+        if (t0 + TB <= w.minlen) {
+            if (loaded != t0) load_tile(t0);
+            float gv[TB];
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                if (rhs) gv[tt] = bload(rg, vg, 4 * (t0 + tt) * M);
+                else gv[tt] = forced ? seed_scale * (zv[tt] - xv[tt]) : 0.f;
+            }
+#pragma unroll
+            for (int tt = TB - 1; tt >= 0; --tt) {
+                const bool m = (posb >> tt) & 1u;
+                const float wt = row16_dot(wT, u);
+                const float y = (t0 + tt + 1 < len) ? pi * fmaf(Ai, u, m ? wt : 0.f) : 0.f;
+                if (lat) u = y + gv[tt];
+            }
+        } else {
+            for (int t = t0 + tl - 1; t >= t0; --t) {
+                const bool run = t < len && lat;
+                const bool m = (t + 1 < len) && ztilde_next(t) > 0.f;
+                const float wt = row16_dot(wT, u);
+                if (run) {
+                    const size_t step = (size_t)b * T + s0 + t;
+                    const float y = (t + 1 < len) ? pi * fmaf(Ai, u, m ? wt : 0.f) : 0.f;
+                    float gk = 0.f;
+                    if (rhs) gk = rhs[step * M + c];
+                    else if (forced) gk = seed_scale * (z[step * M + c] - x[((size_t)b * (T + 1) + s0 + t + 1) * N + c]);
+                    u = y + gk;
+                }
+            }
+        }
+    }
+    if (wmaps) {
+        // Composed for the reverse carry pass (processing order c0+3, c0+2, c0+1, c0):
+        //   slot chain0 + 3:      wave map  Q = (P_3 P_2 P_1 P_0)^T, u_w = the four chunks' walk
+        //   slot chain0 + 3 - j:  prefix    R_j = (P_3 ... P_{4-j})^T, s_j, j = 1..3
+        // so that carry(chain0 + 3 - j) = R_j carry(chain0 + 3) + s_j.  The accumulator layout of
+        // P_n is the A-operand layout of P_n^T; P_3^T as a B operand comes through LDS.
+        __shared__ float lt[16][17];
+        __shared__ float lv[4][16];
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) lt[4 * g + r2][c] = acc[3][r2];
+        lv[g][c] = u;
+        lds_barrier();
+        v4f R1, bv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            R1[q] = lt[c][4 * g + q];   // B layout of P_3^T
+#pragma unroll
+            for (int n = 0; n < 4; ++n) bv[n][q] = c == 0 ? lv[n][4 * g + q] : 0.f;
+        }
+        v4f R2 = {0.f, 0.f, 0.f, 0.f}, R3 = {0.f, 0.f, 0.f, 0.f}, Qw = {0.f, 0.f, 0.f, 0.f};
+        v4f s2 = bv[2], s3 = bv[1], uw = bv[0];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            R2 = mfma16x16x4(acc[2][q], R1[q], R2);
+            s2 = mfma16x16x4(acc[2][q], bv[3][q], s2);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            R3 = mfma16x16x4(acc[1][q], R2[q], R3);
+            s3 = mfma16x16x4(acc[1][q], s2[q], s3);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            Qw = mfma16x16x4(acc[0][q], R3[q], Qw);
+            uw = mfma16x16x4(acc[0][q], s3[q], uw);
+        }
+        // R1 = P_3^T in accumulator layout is the transposed store of acc[3]
+        const v4f outm[4] = {R3, R2, R1, Qw}, outv[4] = {s3, s2, bv[3], uw};
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+            float *P = Pout + (size_t)(chain0 + n) * 256;
+            if (n == 2) {
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) P[c * 16 + 4 * g + r2] = acc[3][r2];
+            } else {
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) P[(4 * g + r2) * 16 + c] = outm[n][r2];
+            }
+            if (c == 0)
+                *reinterpret_cast<float4 *>(vout + (size_t)(chain0 + n) * 16 + 4 * g) =
+                    make_float4(outv[n][0], outv[n][1], outv[n][2], outv[n][3]);
+        }
+        return;
+    }
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        const int cid = chain0 + n;
+        if (cid < nchains && w.plen[n] > 0) {
+            float *P = Pout + (size_t)cid * 256;
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) P[(4 * g + r2) * 16 + c] = acc[n][r2];
+        }
+    }
+    if (okc) vout[(size_t)id * 16 + c] = u;
+}
+
+// M <= 16 reverse fix-up: lam_k from the carry lam_{s1}, written out, with the parameter-
+// gradient partial sums dW[i][j] += lam_i relu(z~_j), dA_i += lam_i z~_i, dh_i += lam_i over
+// the wave's four chains (layout gpart[wave][16][18], the rotated dW columns put back).  A tile
+// row tt is step k = s0 + t0 + tt: z_k, x_k, x_{k+1}, g_k, and z_{k-1} for z~_k.
+template <int TB>
+__global__ __launch_bounds__(64) void k_fixup_rev_plrnn16(const float *__restrict__ A, const float *__restrict__ W,
+                                                         float alpha, int N, const float *__restrict__ gin,
+                                                         float seed_scale, const float *__restrict__ x,
+                                                         const float *__restrict__ z0, const float *__restrict__ z,
+                                                         const float *__restrict__ carry_in,
+                                                         const float *__restrict__ Pm, const float *__restrict__ vmap,
+                                                         float *__restrict__ lam_out, float *__restrict__ gpart, int B,
+                                                         int T, int M, int C, int ncs) {
+    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int nchains = B * ncs;
+    const int chain0 = blockIdx.x * 4;
+    const Chains16 w = chains16(chain0, nchains, ncs, C, T, nullptr, nullptr, nullptr);
+    const int id = chain0 + g;
+    const bool okc = id < nchains;
+    const int b = okc ? id / ncs : 0, s0 = okc ? (id % ncs) * C : 0;
+    int len = 0;
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+        if (n == g) len = w.plen[n];
+    const bool lat = c < M, forced = c < N;
+    int src[16];
+    row_sources(c, src);
+    float wT[16], dW[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        wT[k] = (lat && src[k] < M) ? W[src[k] * M + c] : 0.f;
+        dW[k] = 0.f;
+    }
+    const float pi = p_of(c, N, alpha), Ai = lat ? A[c] : 0.f;
+    float lam = 0.f, dA = 0.f, dh = 0.f;
+    if (len > 0 && lat) {
+        if (!Pm || g == 3) {
+            lam = carry_in[(size_t)id * 16 + c];
+        } else {   // composed wave maps: carry = R carry(chain0 + 3) + s
+            const float4 *R4 = reinterpret_cast<const float4 *>(Pm + (size_t)id * 256 + c * 16);
+            const float4 *w4 = reinterpret_cast<const float4 *>(carry_in + (size_t)(chain0 + 3) * 16);
+            float a0 = vmap[(size_t)id * 16 + c], a1 = 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 rr4 = R4[q], ww = w4[q];
+                a0 = fmaf(rr4.x, ww.x, a0);
+                a1 = fmaf(rr4.y, ww.y, a1);
+                a0 = fmaf(rr4.z, ww.z, a0);
+                a1 = fmaf(rr4.w, ww.w, a1);
+            }
+            lam = a0 + a1;
+        }
+    }
+    // z~ of step s (array index) for this lane
+    auto ztilde = [&](int s) {
+        if (s == 0) return z0 ? z0[(size_t)b * M + c] : (forced ? x[(size_t)b * (T + 1) * N + c] : 0.f);
+        const float zp = z[((size_t)b * T + s - 1) * M + c];
+        if (!forced) return zp;
+        return __fadd_rn(__fmul_rn(pi, zp), __fmul_rn(alpha, x[((size_t)b * (T + 1) + s) * N + c]));
+    };
+    const int cl0 = min(chain0, nchains - 1);
+    const int b0 = cl0 / ncs, s00 = (cl0 % ncs) * C;
+    const size_t row0 = (size_t)b0 * T + s00, xrow0 = (size_t)b0 * (T + 1) + s00;
+    const uint32_t drow = (uint32_t)((size_t)b * T + s0 - row0);
+    const uint32_t dxrow = (uint32_t)((size_t)b * (T + 1) + s0 - xrow0);
+    const auto rz = wave_rsrc(z + row0 * M), rg = wave_rsrc(gin ? gin + row0 * M : z);
+    const auto rx = wave_rsrc(N > 0 ? x + xrow0 * N : z), rl = wave_rsrc(lam_out ? lam_out + row0 * M : z);
+    const uint32_t vz = lat ? 4u * (drow * M + c) : kOffLane;
+    const uint32_t vx = forced ? 4u * (dxrow * N + c) : kOffLane;
+    const uint32_t vg = (gin && lat) ? vz : kOffLane, vl = (lam_out && lat) ? vz : kOffLane;
+    const int last = w.maxlen > 0 ? ((w.maxlen - 1) / TB) * TB : -1;
+    for (int t0 = last; t0 >= 0; t0 -= TB) {
+        const int tl = min(TB, w.maxlen - t0);
+        if (t0 + TB <= w.minlen) {
+            float zv[TB], xv[TB + 1], gv[TB], zt[TB + 1];
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                zv[tt] = bload(rz, vz, 4 * (t0 + tt) * M);
+                xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
+                gv[tt] = bload(rg, vg, 4 * (t0 + tt) * M);
+            }
+            xv[TB] = bload(rx, vx, 4 * (t0 + TB) * N);
+            // z~ of steps s0+t0 .. s0+t0+TB (the last only for the mask of the tile's top step)
+            zt[0] = (len > 0 && lat) ? ztilde(s0 + t0) : 0.f;
+#pragma unroll
+            for (int tt = 1; tt <= TB; ++tt)
+                zt[tt] = forced ? __fadd_rn(__fmul_rn(pi, zv[tt - 1]), __fmul_rn(alpha, xv[tt])) : zv[tt - 1];
+            if (!gin) {
+#pragma unroll
+                for (int tt = 0; tt < TB; ++tt) gv[tt] = forced ? seed_scale * (zv[tt] - xv[tt + 1]) : 0.f;
+            }
+#pragma unroll
+            for (int tt = TB - 1; tt >= 0; --tt) {
+                const int k = s0 + t0 + tt;
+                const bool nxt = k + 1 < T;
+                const bool m = zt[tt + 1] > 0.f;
+                const float wt = row16_dot(wT, lam);
+                const float y = nxt ? pi * fmaf(Ai, lam, m ? wt : 0.f) : 0.f;
+                if (lat) lam = y + gv[tt];
+                bstore_u(rl, __float_as_uint(lam), vl, 4 * (t0 + tt) * M);
+                const float zk = lat ? zt[tt] : 0.f;
+                dA = fmaf(lam, zk, dA);
+                dh += lat ? lam : 0.f;
+                row16_outer(dW, zk > 0.f ? zk : 0.f, lat ? lam : 0.f);
+            }
+        } else {
+            for (int t = t0 + tl - 1; t >= t0; --t) {
+                const bool run = t < len && lat;
+                const int k = s0 + t;
+                const bool nxt = run && k + 1 < T;
+                const bool m = nxt && ztilde(k + 1) > 0.f;
+                const float wt = row16_dot(wT, lam);
+                float zk = 0.f, lr = 0.f;
+                if (run) {
+                    const size_t step = (size_t)b * T + k;
+                    const float y = nxt ? pi * fmaf(Ai, lam, m ? wt : 0.f) : 0.f;
+                    float gk = 0.f;
+                    if (gin) gk = gin[step * M + c];
+                    else if (forced) gk = seed_scale * (z[step * M + c] - x[((size_t)b * (T + 1) + k + 1) * N + c]);
+                    lam = y + gk;
+                    if (lam_out) lam_out[step * M + c] = lam;
+                    zk = ztilde(k);
+                    lr = lam;
+                    dA = fmaf(lam, zk, dA);
+                    dh += lam;
+                }
+                row16_outer(dW, zk > 0.f ? zk : 0.f, lr);
+            }
+        }
+    }
+    // sum over the wave's four chains and write the wave's partial
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) dW[k] += __shfl_xor(dW[k], off, 64);
+        dA += __shfl_xor(dA, off, 64);
+        dh += __shfl_xor(dh, off, 64);
+    }
+    if (g == 0) {
+        float *gp = gpart + ((size_t)blockIdx.x * 16 + c) * 18;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) gp[src[k]] = dW[k];
+        gp[16] = dA;
+        gp[17] = dh;
+    }
+}
+
+// Carries of composed wave maps (four chunks each): one block per sequence, NWV waves.  Each
+// wave composes a contiguous range of maps into one, wave 0 walks the NWV composed maps (LDS),
+// and every wave walks its range again from its own carry, writing the carry of each wave map.
+// Forward: map of wave w at chunk slot 4w, walked w = 0, 1, ...; reverse (adjoint): at slot
+// 4w + 3, walked w = nw - 1, nw - 2, ...; the carry goes to the same slot as the map.
 constexpr int WALK_NWV = 16;
+template <bool REV>
 __global__ __launch_bounds__(WALK_NWV * 64) void k_carry_walk16(const float *__restrict__ P, const float *__restrict__ v,
                                                                float *__restrict__ carry,
                                                                const int *__restrict__ active, int ncs) {
@@ -1501,8 +1913,9 @@ __global__ __launch_bounds__(WALK_NWV * 64) void k_carry_walk16(const float *__r
     const int nw = ncs >> 2, per = (nw + WALK_NWV - 1) / WALK_NWV;
     const int w0 = min(wv * per, nw), w1 = min(w0 + per, nw);
     const float *Pb = P + (size_t)b * ncs * 256, *vb = v + (size_t)b * ncs * 16;
-    auto fetch = [&](int wm, float (&a)[4], float (&vv)[4]) {
-        carry16_fetch<false>(Pb + (size_t)(4 * wm) * 256, vb + (size_t)(4 * wm) * 16, g, c, a, vv);
+    auto slot = [&](int k) { return REV ? 4 * (nw - 1 - k) + 3 : 4 * k; };   // processing position k
+    auto fetch = [&](int k, float (&a)[4], float (&vv)[4]) {
+        carry16_fetch<false>(Pb + (size_t)slot(k) * 256, vb + (size_t)slot(k) * 16, g, c, a, vv);
     };
     float a[PF][4], vv[PF][4];
     // composed map of this wave's range
@@ -1567,7 +1980,7 @@ __global__ __launch_bounds__(WALK_NWV * 64) void k_carry_walk16(const float *__r
             const int wm = k + d;
             if (wm >= w1) break;
             if (c == 0)
-                *reinterpret_cast<float4 *>(carry + ((size_t)b * ncs + 4 * wm) * 16 + 4 * g) =
+                *reinterpret_cast<float4 *>(carry + ((size_t)b * ncs + slot(wm)) * 16 + 4 * g) =
                     make_float4(cur[0], cur[1], cur[2], cur[3]);
             v4f nx = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -2051,11 +2464,12 @@ int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_
     return DEER_OK;
 }
 
-int launch_carry_walk16(const float *P, const float *v, float *carry, const int *active, int B, int ncs,
+int launch_carry_walk16(bool rev, const float *P, const float *v, float *carry, const int *active, int B, int ncs,
                         hipStream_t st) {
     if (ncs % 4) return invalid_arg("wave-map walk needs a chunk count divisible by 4");
     KTimer kt("k_carry", st);
-    hipLaunchKernelGGL(k_carry_walk16, dim3(B), dim3(WALK_NWV * 64), 0, st, P, v, carry, active, ncs);
+    if (rev) hipLaunchKernelGGL(k_carry_walk16<true>, dim3(B), dim3(WALK_NWV * 64), 0, st, P, v, carry, active, ncs);
+    else hipLaunchKernelGGL(k_carry_walk16<false>, dim3(B), dim3(WALK_NWV * 64), 0, st, P, v, carry, active, ncs);
     DEER_LAUNCH_CHECK("k_carry_walk16");
     return DEER_OK;
 }
@@ -2100,6 +2514,36 @@ int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     if (MP == 16) FR(16); else if (MP == 32) FR(32); else FR(64);
 #undef FR
     DEER_LAUNCH_CHECK("k_fixup_rev_plrnn");
+    return DEER_OK;
+}
+
+int launch_adjoint_plrnn16(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *P, float *v,
+                           float *carry, float *lam, float *gpart, int C, int ncs, hipStream_t st) {
+    if (padded(a.M) != 16) return invalid_arg("the register-tiled adjoint needs M <= 16");
+    const int nch = a.B * ncs, grid = (nch + 3) / 4;
+    const bool wm = ncs % 4 == 0;
+    {
+        KTimer kt("k_chunk_product_plrnn", st);
+#define CPR(TBV)                                                                                                     \
+    hipLaunchKernelGGL(k_chunk_product_plrnn16_rev<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, g, z, \
+                       a.x, seed_scale, P, v, a.B, a.T, a.M, C, ncs, (int)wm)
+        if (C <= 16) CPR(16); else CPR(32);
+#undef CPR
+        DEER_LAUNCH_CHECK("k_chunk_product_plrnn16_rev");
+    }
+    int rc;
+    if (wm) rc = launch_carry_walk16(true, P, v, carry, nullptr, a.B, ncs, st);
+    else rc = launch_carry(16, true, P, v, carry, nullptr, nullptr, a.B, ncs, nullptr, st);
+    if (rc) return rc;
+    {
+        KTimer kt("k_fixup_rev_plrnn", st);
+#define FRV(TBV)                                                                                                   \
+    hipLaunchKernelGGL(k_fixup_rev_plrnn16<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, g, seed_scale, \
+                       a.x, a.z0, z, carry, wm ? P : nullptr, wm ? v : nullptr, lam, gpart, a.B, a.T, a.M, C, ncs)
+        if (C <= 16) FRV(16); else FRV(32);
+#undef FRV
+        DEER_LAUNCH_CHECK("k_fixup_rev_plrnn16");
+    }
     return DEER_OK;
 }
 

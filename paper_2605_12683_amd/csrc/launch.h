@@ -35,8 +35,12 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
                                 int ncs, bool wmaps, hipStream_t st);
 // M <= 16 with wave maps (P, v from launch_newton_product_plrnn with wmaps): carries of the
 // wave maps, written to the carry slot of each wave's first chunk
-int launch_carry_walk16(const float *P, const float *v, float *carry, const int *active, int B, int ncs,
+int launch_carry_walk16(bool rev, const float *P, const float *v, float *carry, const int *active, int B, int ncs,
                         hipStream_t st);
+// M <= 16 adjoint: reverse chunk products (masks formed from z), carries, reverse fix-up with
+// the gradient partials of each wave of four chains (gpart[(B ncs + 3) / 4][16][18])
+int launch_adjoint_plrnn16(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *P, float *v,
+                           float *carry, float *lam, float *gpart, int C, int ncs, hipStream_t st);
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
                  uint32_t *norm_bits, int B, int ncs, float *gws, hipStream_t st);
 size_t carry_ws_floats(int MP, int B, int ncs);

@@ -70,7 +70,10 @@ def test_config1_fixed_five_iterations():
 @pytest.mark.parametrize("M,N,B,T,alpha,chunk", [
     (3, 3, 1, 300, 0.1, 0), (3, 3, 2, 300, 0.1, 17), (16, 3, 3, 1000, 0.2, 0), (16, 3, 2, 777, 0.2, 64),
     (20, 4, 2, 513, 0.3, 100), (32, 32, 2, 600, 0.1, 0), (40, 10, 2, 300, 0.3, 33), (64, 64, 2, 400, 0.05, 0),
-    (64, 64, 3, 1000, 0.05, 128), (5, 2, 4, 64, 0.5, 64), (16, 16, 1, 1, 0.2, 0), (8, 8, 2, 2, 0.2, 0)])
+    (64, 64, 3, 1000, 0.05, 128), (5, 2, 4, 64, 0.5, 64), (16, 16, 1, 1, 0.2, 0), (8, 8, 2, 2, 0.2, 0),
+    # chunk counts divisible by 4 (composed wave maps for M <= 16): full tiles, a ragged second
+    # tile, and chunks shorter than a tile
+    (16, 3, 2, 512, 0.2, 16), (7, 3, 3, 640, 0.3, 40), (16, 3, 2, 1000, 0.2, 25)])
 def test_solve_reaches_rollout(M, N, B, T, alpha, chunk):
     """Converged GTF-DEER equals the sequential GTF rollout (unique zero of the residual)."""
     if chunk:
@@ -176,7 +179,9 @@ def test_nonfinite_and_not_converged():
 @pytest.mark.parametrize("M,N,B,T,alpha,chunk", [(3, 3, 1, 300, 0.1, 0), (16, 3, 3, 1000, 0.2, 0),
                                                  (16, 3, 2, 777, 0.2, 64), (20, 4, 2, 513, 0.3, 100),
                                                  (64, 64, 2, 400, 0.05, 0), (40, 10, 2, 300, 0.3, 33),
-                                                 (8, 8, 1, 1, 0.2, 0)])
+                                                 (8, 8, 1, 1, 0.2, 0), (16, 3, 2, 512, 0.2, 16),
+                                                 (7, 3, 3, 640, 0.3, 40), (16, 3, 2, 1000, 0.2, 25),
+                                                 (16, 16, 3, 256, 0.1, 32)])
 def test_adjoint_and_grads(M, N, B, T, alpha, chunk):
     """lam and dL/dtheta at the same float32 trajectory (the oracle's fixed point rounded to
     float32); both sides take the ReLU decision in float32."""

@@ -337,11 +337,33 @@ static size_t diag_bytes(int B, int T, int M, int K, int op) {
 // exceeds step_bound (1 + max|z|), is not kept and the sequence is retried with gamma < 1;
 // gamma returns to 1 over accepted updates.  gamma = 1 is the exact Newton step, gamma = 0
 // the fixed-point step z_t <- F(z~_{t-1}); every gamma keeps the fixed point and the prefix
-// property.  The host queues passes in batches and reads the active flags once per batch;
-// a sequence frozen inside a batch makes the rest of the batch's kernels skip it.
+// property.  The host queues passes in batches and reads the active flags of a batch while
+// the next batch already runs (the pass-end control clears a pinned host copy of the flags
+// too; an event per batch tells the host which passes are complete), so the device does not
+// wait for the host; a sequence frozen inside a batch makes the rest of the queued kernels
+// skip it, and once every sequence is frozen the passes still queued skip everything.
 constexpr float kDefaultStepBound = 1e3f;
 constexpr NewtonDamp kDamp = {1.f / 64, 4.f, 4.f, 1e-4f};
-constexpr int kFirstBatch = 4, kBatch = 2;
+constexpr int kFirstBatch = 4, kBatch = 1;
+
+// pinned, device-coherent host copy of the active flags (per host thread, grown on demand,
+// kept for the life of the process)
+struct ActPoll {
+    int *host = nullptr;
+    size_t cap = 0;
+};
+static thread_local ActPoll t_poll;
+static int poll_flags(int B, int **flags) {
+    if ((size_t)B > t_poll.cap) {
+        if (t_poll.host) (void)hipHostFree(t_poll.host);
+        t_poll.host = nullptr;
+        t_poll.cap = 0;
+        DEER_HIP(hipHostMalloc((void **)&t_poll.host, (size_t)B * sizeof(int), hipHostMallocCoherent));
+        t_poll.cap = (size_t)B;
+    }
+    *flags = t_poll.host;
+    return DEER_OK;
+}
 
 template <class Update>
 static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int ncs, const NewtonCtl &ctl, float *z,
@@ -365,23 +387,56 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
         }
         return DEER_OK;
     }
-    const NewtonDev &nd = ctl.nd;
+    NewtonDev nd = ctl.nd;
+    if (!nd.hact && (rc = poll_flags(B, &nd.hact))) return rc;
+    int *const hact = nd.hact;
+    for (int b = 0; b < B; ++b) hact[b] = 1;   // no kernel of this stream that writes it is pending
     if ((rc = launch_ctl_init(nd, ctl.seq, B, st))) return rc;
-    int passes = 0, batch = kFirstBatch;
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    auto done_events = [&]() {
+        for (hipEvent_t &e : ev)
+            if (e) (void)hipEventDestroy(e);
+    };
+    for (hipEvent_t &e : ev) {
+        const hipError_t err = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+        if (err != hipSuccess) {
+            done_events();
+            return hip_fail(err, "hipEventCreateWithFlags");
+        }
+    }
+    auto check = [&](hipError_t err, const char *what) {
+        if (err == hipSuccess) return 0;
+        done_events();
+        return hip_fail(err, what);
+    };
+    int passes = 0, batch = kFirstBatch, k = 0;
     while (passes < max_iter) {
         const int n = batch < max_iter - passes ? batch : max_iter - passes;
-        for (int k = 0; k < n; ++k) {
-            if ((rc = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt))) return rc;
-            if (!ctl.fused && (rc = launch_seq_ctl(ctl.chain_bits, nd, B, ncs, o->tol, bound, kDamp, st))) return rc;
+        for (int j = 0; j < n; ++j) {
+            rc = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt);
+            if (!rc && !ctl.fused) rc = launch_seq_ctl(ctl.chain_bits, nd, B, ncs, o->tol, bound, kDamp, st);
+            if (rc) {
+                done_events();
+                return rc;
+            }
         }
         passes += n;
-        DEER_HIP(hipMemcpyAsync(act.data(), nd.act, B * sizeof(int), hipMemcpyDeviceToHost, st));
-        DEER_HIP(hipStreamSynchronize(st));
-        bool any = false;
-        for (int b = 0; b < B; ++b) any |= act[b] != 0;
-        if (!any) break;
+        if ((rc = check(hipEventRecord(ev[k & 1], st), "hipEventRecord"))) return rc;
         batch = kBatch;
+        // Short passes (the fused M <= 16 path): the flags as of the end of the previous batch,
+        // read while this one runs (they only go from 1 to 0, so a later pass having cleared
+        // more is harmless).  Long passes: this batch's flags, as the host wait is then small
+        // next to a pass and a pass queued past convergence is not.
+        const int kc = ctl.fused ? k - 1 : k;
+        if (kc >= 0) {
+            if ((rc = check(hipEventSynchronize(ev[kc & 1]), "hipEventSynchronize"))) return rc;
+            bool any = false;
+            for (int b = 0; b < B; ++b) any |= __atomic_load_n(hact + b, __ATOMIC_ACQUIRE) != 0;
+            if (!any) break;
+        }
+        ++k;
     }
+    done_events();
     std::vector<uint32_t> h(7 * (size_t)B);
     DEER_HIP(hipMemcpyAsync(h.data(), ctl.blk, h.size() * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
     DEER_HIP(hipStreamSynchronize(st));
@@ -438,6 +493,7 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     // M <= 16: the fix-up also takes the pass-end control of the adaptive loop
     NewtonCtl ctl = w.ctl;
     ctl.fused = w.MP == 16 && o->fixed_iters <= 0;
+    if (ctl.fused && (rc = poll_flags(B, &ctl.nd.hact))) return rc;
     const FusedCtl fc{ctl.nd, ctl.seq, o->tol, o->step_bound == 0.f ? kDefaultStepBound : o->step_bound, kDamp};
     auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za) -> int {
         int r;

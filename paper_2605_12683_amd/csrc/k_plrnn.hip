@@ -886,11 +886,13 @@ __device__ __forceinline__ void seq_decide(int b, uint32_t e, uint32_t zm, const
         if (om > 0.f) om = om / dp.shrink < dp.floor ? 0.f : om / dp.shrink;
         if (ef < tol) {
             nd.act[b] = 0;
+            if (nd.hact) nd.hact[b] = 0;
             nd.status[b] = 1;
         }
     } else if (om >= 1.f) {
         nd.norm[b] = ef;
         nd.act[b] = 0;
+        if (nd.hact) nd.hact[b] = 0;
         nd.status[b] = 2;
     } else {
         om = om == 0.f ? dp.first : fminf(1.f, om * dp.grow);

@@ -57,6 +57,7 @@ struct NewtonDev {
     int *it;        // accepted updates
     float *norm;    // max |Delta| of the last accepted (or final) update
     int *status;    // 0 running, 1 converged, 2 non-finite
+    int *hact;      // pinned host copy of act, cleared together with act (may be null)
 };
 struct NewtonDamp {
     float first, grow, shrink, floor;

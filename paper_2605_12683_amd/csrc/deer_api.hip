@@ -101,6 +101,22 @@ __global__ void k_fill_i32(int *p, int n, int v) {
     const int e = blockIdx.x * blockDim.x + threadIdx.x;
     if (e < n) p[e] = v;
 }
+// the iterate of sequence b ended in the second buffer when sel[b] is set: copy it back
+__global__ void k_copy_sel(float *__restrict__ z, const float *__restrict__ zalt, const int *__restrict__ sel,
+                           size_t seq_elems) {
+    const int b = blockIdx.y;
+    if (!sel[b]) return;
+    float *d = z + (size_t)b * seq_elems;
+    const float *s = zalt + (size_t)b * seq_elems;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    if ((seq_elems & 3) == 0 && ((uintptr_t)d & 15) == 0 && ((uintptr_t)s & 15) == 0) {
+        const size_t n4 = seq_elems >> 2;
+        for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n4; e += stride)
+            reinterpret_cast<float4 *>(d)[e] = reinterpret_cast<const float4 *>(s)[e];
+    } else {
+        for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < seq_elems; e += stride) d[e] = s[e];
+    }
+}
 __global__ void k_fill_f32(float *p, size_t n, float v) {
     for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n; e += (size_t)gridDim.x * blockDim.x) p[e] = v;
 }
@@ -157,6 +173,8 @@ static int choose_chunk(int B, int T, int MP) {
     const long maxc = MP <= 32 ? 1024 : 512;
     const long minC = (T + maxc - 1) / maxc;
     if (C < minC) C = minC;
+    // M <= 16: whole 16-step tiles (the register-tiled kernels run a partial tile step by step)
+    if (MP == 16) C = (C + 15) / 16 * 16;
     if (C > T) C = T;
     return (int)C;
 }
@@ -437,18 +455,23 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
         ++k;
     }
     done_events();
+    // sequences whose iterate ended in the second buffer are copied back on the device (one
+    // launch, no host decision), then the control block is read once
+    {
+        const size_t n4 = (seq_elems + 3) / 4;
+        const unsigned gx = (unsigned)((n4 + 255) / 256 < 256 ? (n4 + 255) / 256 : 256);
+        hipLaunchKernelGGL(k_copy_sel, dim3(gx, B), dim3(256), 0, st, z, (const float *)ctl.zalt,
+                           (const int *)nd.sel, seq_elems);
+        DEER_LAUNCH_CHECK("k_copy_sel");
+    }
     std::vector<uint32_t> h(7 * (size_t)B);
     DEER_HIP(hipMemcpyAsync(h.data(), ctl.blk, h.size() * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
     DEER_HIP(hipStreamSynchronize(st));
-    const size_t seq_bytes = seq_elems * sizeof(float);
     for (int b = 0; b < B; ++b) {
         act[b] = (int)h[b];
         it[b] = (int)h[4 * (size_t)B + b];
         memcpy(&norm[b], &h[5 * (size_t)B + b], 4);
         if (h[6 * (size_t)B + b] == 2u) nonfinite = true;
-        if (h[2 * (size_t)B + b])   // the iterate ended in the second buffer
-            DEER_HIP(hipMemcpyAsync(z + b * seq_elems, ctl.zalt + b * seq_elems, seq_bytes, hipMemcpyDeviceToDevice,
-                                    st));
     }
     return DEER_OK;
 }

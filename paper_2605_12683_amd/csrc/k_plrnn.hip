@@ -2384,7 +2384,7 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
         hipLaunchKernelGGL(k_newton_product_plrnn64u, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0,
                            z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
     } else if (MP == 16) {
-        if (C <= 16)
+        if (C % 32)
             hipLaunchKernelGGL(k_newton_product_plrnn16<16>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
                                a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs,
                                (int)wmaps);
@@ -2496,7 +2496,7 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     FusedCtl fcv{};
     if (fc) fcv = *fc;
     if (MP == 16) {
-        if (C <= 16) FX16(16); else FX16(32);
+        if (C % 32) FX16(16); else FX16(32);
     } else if (MP == 32) FX(32); else FX(64);
 #undef FX16
 #undef FX
@@ -2529,7 +2529,7 @@ int launch_adjoint_plrnn16(const PlrnnArgs &a, const float *g, float seed_scale,
 #define CPR(TBV)                                                                                                     \
     hipLaunchKernelGGL(k_chunk_product_plrnn16_rev<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, g, z, \
                        a.x, seed_scale, P, v, a.B, a.T, a.M, C, ncs, (int)wm)
-        if (C <= 16) CPR(16); else CPR(32);
+        if (C % 32) CPR(16); else CPR(32);
 #undef CPR
         DEER_LAUNCH_CHECK("k_chunk_product_plrnn16_rev");
     }
@@ -2542,7 +2542,7 @@ int launch_adjoint_plrnn16(const PlrnnArgs &a, const float *g, float seed_scale,
 #define FRV(TBV)                                                                                                   \
     hipLaunchKernelGGL(k_fixup_rev_plrnn16<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, g, seed_scale, \
                        a.x, a.z0, z, carry, wm ? P : nullptr, wm ? v : nullptr, lam, gpart, a.B, a.T, a.M, C, ncs)
-        if (C <= 16) FRV(16); else FRV(32);
+        if (C % 32) FRV(16); else FRV(32);
 #undef FRV
         DEER_LAUNCH_CHECK("k_fixup_rev_plrnn16");
     }

@@ -522,9 +522,10 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
 // are formed with DPP row rotations (no LDS, no barrier).  Steps go in tiles of TB.  In a tile
 // that all four chains run to its end (every tile but a ragged chunk's last) all loads of the
 // tile are issued at once through buffer resources (one lane offset for all of them), the
-// residual of every step of the tile, which does not depend on the recurrence, is formed and
-// stored first, and the serial part then runs from registers, with the matrix-core updates of
-// the four chains free of branches so that they interleave.  Other tiles go step by step.
+// residual of every step of the tile, which does not depend on the recurrence, is formed
+// first, and the serial part then runs from registers, with the matrix-core updates of the
+// four chains free of branches so that they interleave.  Other tiles go step by step.  The
+// residual and the masks stay in registers: the fix-up forms them again from z and x.
 // ---------------------------------------------------------------------------------------
 
 // lane l of each 16-lane row receives v from lane row_src(l, K) of the same row
@@ -663,7 +664,7 @@ template <int TB>
 __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
     const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
     const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
-    const int *__restrict__ zsel, float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout,
+    const int *__restrict__ zsel, float *__restrict__ Pout,
     float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
     int ncs, int wmaps) {
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
@@ -715,11 +716,10 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
     const size_t row0 = (size_t)b0 * T + s00, xrow0 = (size_t)b0 * (T + 1) + s00;
     const uint32_t drow = (uint32_t)((size_t)b * T + s0 - row0), dxrow = (uint32_t)((size_t)b * (T + 1) + s0 - xrow0);
     const float *zw = cur_iter(zbuf, zalt, zsel, b0);
-    const auto rz = wave_rsrc(zw + row0 * M), rr = wave_rsrc(r_out + row0 * M), rm = wave_rsrc(masks + row0);
+    const auto rz = wave_rsrc(zw + row0 * M);
     const auto rx = wave_rsrc(N > 0 ? x + xrow0 * N : zw);
     const uint32_t vz = lat ? 4u * (drow * M + c) : kOffLane;
     const uint32_t vx = forced ? 4u * (dxrow * N + c) : kOffLane;
-    const uint32_t vm = c == 0 ? 4u * drow : kOffLane;
     float u = 0.f;
     for (int t0 = 0; t0 < w.maxlen; t0 += TB) {
         const int tl = min(TB, w.maxlen - t0);
@@ -742,9 +742,6 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
                 const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
                 zprev = zv[tt];
                 zv[tt] = zv[tt] - F;
-                bstore_u(rr, __float_as_uint(zv[tt]), vz, 4 * (t0 + tt) * M);
-                const uint64_t bal = __ballot(pos);
-                bstore_u(rm, (uint32_t)((bal >> (16 * g)) & 0xffffull), vm, 4 * (t0 + tt));
             }
             // serial part: chunk products and chunk-local solutions
 #pragma unroll
@@ -787,11 +784,6 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
                 const uint64_t bal = __ballot(pos);
                 const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
                 const float r = zcur - F;
-                if (t < len) {
-                    const size_t step = (size_t)b * T + s;
-                    if (lat) r_out[step * M + c] = r;
-                    if (c == 0) masks[step] = (uint32_t)((bal >> (16 * g)) & 0xffffull);
-                }
 #pragma unroll
                 for (int n = 0; n < 4; ++n)
                     if (t < w.plen[n]) acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
@@ -921,11 +913,17 @@ __device__ __forceinline__ void seq_arrive(const FusedCtl &fc, int b, int cnt, i
     __hip_atomic_store(blk, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// M <= 16 forward fix-up.  The residual and the masks are formed again here from z and x (the
+// same operations as the forward pass, so the same values), which saves writing them there
+// and reading them here; Delta_t = gamma (diag(d) + W p diag(m_t)) Delta_{t-1} - r_t from the
+// chunk's carry, z + Delta written to the other iterate buffer, per-chain max |Delta| and max
+// |z|, and (with fc.seq) the pass-end control of the sequence.
 template <int TB>
 __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restrict__ A, const float *__restrict__ W,
-                                                          float alpha, int N, const uint32_t *__restrict__ masks,
-                                                          const float *__restrict__ r, const float *__restrict__ carry_in,
-                                                          float *zbuf, float *zalt, const int *__restrict__ zsel,
+                                                          const float *__restrict__ h, float alpha, int N,
+                                                          const float *__restrict__ x, const float *__restrict__ z0,
+                                                          const float *__restrict__ carry_in, float *zbuf,
+                                                          float *zalt, const int *__restrict__ zsel,
                                                           uint32_t *__restrict__ chain_bits,
                                                           const int *__restrict__ active,
                                                           const float *__restrict__ gamma, int B, int T, int M, int C,
@@ -947,13 +945,17 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
             len = w.plen[n];
             gm = w.gam[n];
         }
-    const bool lat = c < M;
+    const bool lat = c < M, forced = c < N;
     int src[16];
     row_sources(c, src);
-    float wp[16];
+    float wr[16], wp[16];
 #pragma unroll
-    for (int k = 0; k < 16; ++k) wp[k] = (lat && src[k] < M) ? W[c * M + src[k]] * p_of(src[k], N, alpha) : 0.f;
-    const float d = lat ? A[c] * p_of(c, N, alpha) : 0.f;
+    for (int k = 0; k < 16; ++k) {
+        wr[k] = (lat && src[k] < M) ? W[c * M + src[k]] : 0.f;
+        wp[k] = wr[k] * p_of(src[k], N, alpha);
+    }
+    const float Ai = lat ? A[c] : 0.f, hi = (lat && h) ? h[c] : 0.f;
+    const float pi = p_of(c, N, alpha), d = Ai * pi;
     float D = 0.f;
     if (len > 0 && lat) {
         if (!Pm || g == 0) {
@@ -975,29 +977,47 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
     }
     const float *zin = cur_iter(zbuf, zalt, zsel, b);
     float *zout = next_iter(zbuf, zalt, zsel, b);
+    float zprev = 0.f;   // z_{s-1} of the first step (the initial state at s = 0)
+    if (len > 0 && lat) {
+        if (s0 == 0) zprev = z0 ? z0[(size_t)b * M + c] : (forced ? x[(size_t)b * (T + 1) * N + c] : 0.f);
+        else zprev = zin[((size_t)b * T + s0 - 1) * M + c];
+    }
     const int cl0 = min(chain0, nchains - 1);   // a wave past the last chain touches no memory
-    const int b0 = cl0 / ncs;
-    const size_t row0 = (size_t)b0 * T + (size_t)(cl0 % ncs) * C;
+    const int b0 = cl0 / ncs, s00 = (cl0 % ncs) * C;
+    const size_t row0 = (size_t)b0 * T + s00, xrow0 = (size_t)b0 * (T + 1) + s00;
     const uint32_t drow = (uint32_t)((size_t)b * T + s0 - row0);
-    const auto rr = wave_rsrc(r + row0 * M), rm = wave_rsrc(masks + row0);
+    const uint32_t dxrow = (uint32_t)((size_t)b * (T + 1) + s0 - xrow0);
     const auto rzi = wave_rsrc(cur_iter(zbuf, zalt, zsel, b0) + row0 * M);
     const auto rzo = wave_rsrc(next_iter(zbuf, zalt, zsel, b0) + row0 * M);
-    const uint32_t vz = lat ? 4u * (drow * M + c) : kOffLane, vm = 4u * drow;
+    const auto rx = wave_rsrc(N > 0 ? x + xrow0 * N : zin);
+    const uint32_t vz = lat ? 4u * (drow * M + c) : kOffLane;
+    const uint32_t vx = forced ? 4u * (dxrow * N + c) : kOffLane;
     uint32_t emax = 0u, zmax = 0u;
     for (int t0 = 0; t0 < w.maxlen; t0 += TB) {
         const int tl = min(TB, w.maxlen - t0);
         if (w.onebuf && t0 + TB <= w.minlen) {
-            float rv[TB], zv[TB];
-            uint32_t mv[TB];
+            float zv[TB], rv[TB];
 #pragma unroll
             for (int tt = 0; tt < TB; ++tt) {
-                rv[tt] = bload(rr, vz, 4 * (t0 + tt) * M);
                 zv[tt] = bload(rzi, vz, 4 * (t0 + tt) * M);
-                mv[tt] = bload_u(rm, vm, 4 * (t0 + tt));
+                rv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);   // x of the step, replaced by r below
+            }
+            // residual and masks of the tile (as in the forward pass)
+            uint32_t mb = 0u;
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                const int s = s0 + t0 + tt;
+                const float zt =
+                    (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, rv[tt]));
+                const bool pos = zt > 0.f;
+                mb |= (pos ? 1u : 0u) << tt;
+                const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
+                zprev = zv[tt];
+                rv[tt] = zv[tt] - F;
             }
 #pragma unroll
             for (int tt = 0; tt < TB; ++tt) {
-                const bool m = (mv[tt] >> c) & 1u;
+                const bool m = (mb >> tt) & 1u;
                 const float y = fmaf(d, D, row16_dot(wp, m ? D : 0.f));
                 D = fmaf(gm, y, -rv[tt]);
                 const float zc = zv[tt];
@@ -1009,22 +1029,26 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
         } else {
             for (int t = t0; t < t0 + tl; ++t) {
                 const bool run = t < len && lat;
-                const size_t step = (size_t)b * T + s0 + t;
-                float rc = 0.f, zc = 0.f;
-                uint32_t mc = 0u;
+                const int s = s0 + t;
+                const size_t step = (size_t)b * T + s;
+                float zc = 0.f, xb = 0.f;
                 if (run) {
-                    rc = r[step * M + c];
                     zc = zin[step * M + c];
-                    mc = masks[step];
+                    if (forced && s > 0) xb = x[((size_t)b * (T + 1) + s) * N + c];
                 }
-                const bool m = run && ((mc >> c) & 1u);
-                const float y = fmaf(d, D, row16_dot(wp, m ? D : 0.f));
+                float zt = 0.f;
+                if (run) zt = (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xb));
+                const bool pos = zt > 0.f;
+                const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
+                const float rc = zc - F;
+                const float y = fmaf(d, D, row16_dot(wp, (run && pos) ? D : 0.f));
                 if (run) {
                     D = fmaf(gm, y, -rc);
                     zout[step * M + c] = zc + D;
                     const uint32_t ab = abs_bits(D), zb = abs_bits(zc);
                     emax = emax > ab ? emax : ab;
                     zmax = zmax > zb ? zmax : zb;
+                    zprev = zc;
                 }
             }
         }
@@ -1943,7 +1967,7 @@ __global__ __launch_bounds__(WALK_NWV * 64) void k_carry_walk16(const float *__r
                 }
                 S = ns;
                 t = nt;
-                fetch(min(k + d + PF, w1 - 1), a[d], vv[d]);
+                if (per > PF) fetch(min(k + d + PF, w1 - 1), a[d], vv[d]);   // else kept for the re-walk
             }
         }
     }
@@ -1974,8 +1998,10 @@ __global__ __launch_bounds__(WALK_NWV * 64) void k_carry_walk16(const float *__r
     v4f cur;
 #pragma unroll
     for (int r = 0; r < 4; ++r) cur[r] = c == 0 ? lsc[wv][4 * g + r] : 0.f;
+    if (per > PF) {
 #pragma unroll
-    for (int d = 0; d < PF; ++d) fetch(min(w0 + d, w1 - 1), a[d], vv[d]);
+        for (int d = 0; d < PF; ++d) fetch(min(w0 + d, w1 - 1), a[d], vv[d]);
+    }
     for (int k = w0; k < w1; k += PF) {
 #pragma unroll
         for (int d = 0; d < PF; ++d) {
@@ -1992,7 +2018,7 @@ __global__ __launch_bounds__(WALK_NWV * 64) void k_carry_walk16(const float *__r
                 for (int r = 0; r < 4; ++r) nx[r] += vv[d][r];
             }
             cur = nx;
-            fetch(min(wm + PF, w1 - 1), a[d], vv[d]);
+            if (per > PF) fetch(min(wm + PF, w1 - 1), a[d], vv[d]);
         }
     }
 }
@@ -2386,12 +2412,10 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
     } else if (MP == 16) {
         if (C % 32)
             hipLaunchKernelGGL(k_newton_product_plrnn16<16>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
-                               a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs,
-                               (int)wmaps);
+                               a.x, a.z0, z, zalt, zsel, P, v, active, gamma, a.B, a.T, a.M, C, ncs, (int)wmaps);
         else
             hipLaunchKernelGGL(k_newton_product_plrnn16<32>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
-                               a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs,
-                               (int)wmaps);
+                               a.x, a.z0, z, zalt, zsel, P, v, active, gamma, a.B, a.T, a.M, C, ncs, (int)wmaps);
     } else if (MP == 32) NP(32); else NP(64);
 #undef NP
     DEER_LAUNCH_CHECK("k_newton_product_plrnn");
@@ -2487,8 +2511,8 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
 #define FX(MPV)                                                                                                       \
     hipLaunchKernelGGL(k_fixup_fwd_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, carry_in, \
                        z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
-#define FX16(TBV)                                                                                              \
-    hipLaunchKernelGGL(k_fixup_fwd_plrnn16<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, \
+#define FX16(TBV)                                                                                                 \
+    hipLaunchKernelGGL(k_fixup_fwd_plrnn16<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, \
                        carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs, Pm, vm, fcv)
     if (Pm && (MP != 16 || ncs % 4))
         return invalid_arg("composed wave maps need M <= 16 and a chunk count divisible by 4");

@@ -19,11 +19,14 @@ __device__ __forceinline__ float p_at(int i, int N, float alpha) { return i < N 
 
 // ---------------------------------------------------------------------------------------
 // residual + masks.  Block of 256 threads (4 waves), TT rows (b, t) per tile, grid-stride
-// over tiles.  The hidden pre-activations u = W2 z~ + h2 that decide the masks are summed on
-// the VALU in a fixed order (left to right from h2, a rounding after every multiply and add);
-// F = A z~ + W1 relu(u) + h1 is a [M x L] x [L x TT] product on the matrix cores with the
-// k range split over the 4 waves and the partial tiles summed through LDS.
-// dynamic LDS: zt[TT][MP] | ru[TT][LQ] | W1[MP][LQ] | partial F tiles [4][NI][64][4]
+// over tiles; the inputs of the next tile are loaded into registers while a tile is
+// processed.  The hidden pre-activations u = W2 z~ + h2 that decide the masks are summed on
+// the VALU in a fixed order (left to right from h2, a rounding after every multiply and add),
+// thread j holding W2 row j and the TT sums of hidden unit j, the TT values z~_k read from LDS
+// as four 16-byte broadcasts per k; F = A z~ + W1 relu(u) + h1 is a [M x L] x [L x TT]
+// product on the matrix cores with the k range split over the 4 waves, and the partial tiles
+// are summed by the threads that loaded those four latents of the row (and keep z for r).
+// dynamic LDS: z~^T[MP][TT] | ru[TT][LQ] | W1[MP][LQ] | partial F [4][NI][64][4]
 // (LQ = L rounded up to 16, + 4 so that rows stay 16-byte aligned and spread over banks)
 // ---------------------------------------------------------------------------------------
 constexpr int SH_TT = 16;
@@ -35,75 +38,125 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
                                                         const int *__restrict__ zsel, float *__restrict__ F_out,
                                                         float *__restrict__ r_out, uint32_t *__restrict__ masks,
                                                         const int *__restrict__ active) {
-    constexpr int NI = MP / 16;
+    constexpr int NI = MP / 16, TT = SH_TT, NT4 = TT * MP / 4;   // threads owning 4 latents of a row
+    static_assert(NT4 <= 256 && TT == 16, "tile shape");
     extern __shared__ __align__(16) float smem[];
-    const int M = a.M, L = a.L, T = a.T, LQ = sh_LQ(L);
-    float *zt = smem;                    // [SH_TT][MP], zero padded
-    float *ru = zt + SH_TT * MP;         // [SH_TT][LQ], zero padded
-    float *w1s = ru + SH_TT * LQ;        // [MP][LQ] = W1, zero padded
+    const int M = a.M, L = a.L, T = a.T, N = a.N, LQ = sh_LQ(L);
+    float *zT = smem;                    // [MP][TT]  z~ transposed
+    float *ru = zT + MP * TT;            // [TT][LQ], zero padded
+    float *w1s = ru + TT * LQ;           // [MP][LQ] = W1, zero padded
     v4f *red = reinterpret_cast<v4f *>(w1s + MP * LQ);   // [4][NI][64]
+    __shared__ int rowok[SH_TT];         // row of the tile exists and its sequence is active
     const int tid = threadIdx.x;
     const int lane = tid & 63, wv = tid >> 6, g = lane >> 4, c = lane & 15;
     const int LW = (L + 31) / 32;
+    const float p = __fsub_rn(1.0f, a.alpha);
     for (int e = tid; e < MP * LQ; e += 256) {
         const int i = e / LQ, l = e % LQ;
         w1s[e] = (i < M && l < L) ? a.W1[i * L + l] : 0.f;
     }
-    for (int e = tid; e < SH_TT * LQ; e += 256) ru[e] = 0.f;
+    for (int e = tid; e < TT * LQ; e += 256) ru[e] = 0.f;
     const long total = (long)a.B * T;
-    const long ntiles = (total + SH_TT - 1) / SH_TT;
+    const long ntiles = (total + TT - 1) / TT;
     const int njg = (L + 15) / 16;
-    for (long tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-        const long row0 = tile * SH_TT;
-        __syncthreads();
-        for (int e = tid; e < SH_TT * MP; e += 256) {
-            const int tt = e / MP, i = e % MP;
-            const long row = row0 + tt;
-            float v = 0.f;
-            if (row < total && i < M) {
-                const int b = (int)(row / T), s = (int)(row % T);
-                v = forced_state(a.x, a.z0, cur_iter(zbuf, zalt, zsel, b), b, s, i, T, M, a.N, a.alpha);
+    // the tile's inputs owned by this thread (tid < NT4): latents i0..i0+3 of row rc, the same
+    // elements whose residual it writes at the end of the tile
+    const int rc = tid / (MP / 4), i0 = 4 * (tid % (MP / 4));
+    float pz[4], px[4], pc[4], cz[4];   // z_{s-1} (or the initial state at s = 0), x_s, z_s
+    auto fetch = [&](long tile) {
+        const long row = tile * TT + rc;
+        const bool ok = tid < NT4 && tile < ntiles && row < total;
+        const int b = ok ? (int)(row / T) : 0, s = ok ? (int)(row % T) : 0;
+        const float *z = cur_iter(zbuf, zalt, zsel, b);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int i = i0 + r;
+            pz[r] = 0.f;
+            px[r] = 0.f;
+            pc[r] = 0.f;
+            if (ok && i < M) {
+                if (s == 0) {
+                    pz[r] = a.z0 ? a.z0[(size_t)b * M + i] : (i < N ? a.x[(size_t)b * (T + 1) * N + i] : 0.f);
+                } else {
+                    pz[r] = z[((size_t)b * T + s - 1) * M + i];
+                    if (i < N) px[r] = a.x[((size_t)b * (T + 1) + s) * N + i];
+                }
+                pc[r] = z[((size_t)b * T + s) * M + i];
             }
-            zt[e] = v;
         }
+    };
+    // W2 rows of this thread's hidden units stay in registers when L <= 256
+    float w2r[MP];
+    float h2j = 0.f;
+    auto load_w2 = [&](int j) {
+        const bool jok = j < L;
+#pragma unroll
+        for (int k = 0; k < MP; ++k) w2r[k] = (jok && k < M) ? a.W2[(size_t)j * M + k] : 0.f;
+        h2j = (jok && a.h2) ? a.h2[j] : 0.f;
+    };
+    if (L <= 256) load_w2(tid);
+    long tile = blockIdx.x;
+    fetch(tile);
+    for (; tile < ntiles; tile += gridDim.x) {
+        const long row0 = tile * TT;
+        __syncthreads();   // the previous tile is done with zT, zc, ru and red
+        if (tid < NT4) {
+            const long row = row0 + rc;
+            const bool later = row < total && (int)(row % T) > 0;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int i = i0 + r;
+                float zt = pz[r];
+                if (later && i < N) zt = __fadd_rn(__fmul_rn(p, pz[r]), __fmul_rn(a.alpha, px[r]));
+                zT[i * TT + rc] = zt;
+                cz[r] = pc[r];
+            }
+        }
+        if (tid < TT) {
+            const long row = row0 + tid;
+            rowok[tid] = row < total && (!active || active[row / T]);
+        }
+        fetch(tile + gridDim.x);
         __syncthreads();
         // hidden pre-activations: left to right in k from h2, separate roundings.  The zero
         // padding adds exact zeros, so the value is the one of the unpadded sum.
         for (int jb = 0; jb < L; jb += 256) {
             const int j = jb + tid;
             const bool jok = j < L;
-            float w2r[MP];
+            if (L > 256) load_w2(j);
+            float u[TT];
 #pragma unroll
-            for (int k = 0; k < MP; ++k) w2r[k] = (jok && k < M) ? a.W2[(size_t)j * M + k] : 0.f;
-            const float h2j = (jok && a.h2) ? a.h2[j] : 0.f;
-            // RG rows at a time: independent chains interleaved (each sum is serial in k)
-            constexpr int RG = 4;
-            for (int tt0 = 0; tt0 < SH_TT; tt0 += RG) {
-                float u[RG];
+            for (int t = 0; t < TT; ++t) u[t] = h2j;
 #pragma unroll
-                for (int q = 0; q < RG; ++q) u[q] = h2j;
+            for (int k = 0; k < MP; ++k) {
+                const float4 *z4 = reinterpret_cast<const float4 *>(zT + k * TT);
 #pragma unroll
-                for (int k = 0; k < MP; ++k)
+                for (int t4 = 0; t4 < TT / 4; ++t4) {
+                    const float4 v = z4[t4];
+                    u[4 * t4] = __fadd_rn(u[4 * t4], __fmul_rn(w2r[k], v.x));
+                    u[4 * t4 + 1] = __fadd_rn(u[4 * t4 + 1], __fmul_rn(w2r[k], v.y));
+                    u[4 * t4 + 2] = __fadd_rn(u[4 * t4 + 2], __fmul_rn(w2r[k], v.z));
+                    u[4 * t4 + 3] = __fadd_rn(u[4 * t4 + 3], __fmul_rn(w2r[k], v.w));
+                }
+            }
 #pragma unroll
-                    for (int q = 0; q < RG; ++q) u[q] = __fadd_rn(u[q], __fmul_rn(w2r[k], zt[(tt0 + q) * MP + k]));
-#pragma unroll
-                for (int q = 0; q < RG; ++q) {
-                    const int tt = tt0 + q;
-                    const bool pos = jok && u[q] > 0.f;
-                    if (jok) ru[tt * LQ + j] = pos ? u[q] : 0.f;
-                    const uint64_t bal = __ballot(pos);
-                    const long row = row0 + tt;
-                    if (masks && row < total && (lane == 0 || lane == 32)) {
-                        const int b = (int)(row / T);
-                        if (!active || active[b]) {
-                            const int word = (jb + tid) / 32;
-                            if (word < LW) masks[(size_t)row * LW + word] = (uint32_t)(bal >> lane);
-                        }
-                    }
+            for (int t = 0; t < TT; ++t)
+                if (jok) ru[t * LQ + j] = u[t] > 0.f ? u[t] : 0.f;
+        }
+        __syncthreads();
+        // mask words from relu(u) > 0 (= u > 0), rows of active sequences only
+        if (masks) {
+            for (int jb = 0; jb < L; jb += 256) {
+                const int j = jb + tid;
+                const int word = j / 32;
+#pragma unroll 4
+                for (int t = 0; t < TT; ++t) {
+                    const uint64_t bal = __ballot(j < L && ru[t * LQ + j] > 0.f);
+                    if (rowok[t] && (lane == 0 || lane == 32) && word < LW)
+                        masks[(size_t)(row0 + t) * LW + word] = (uint32_t)(bal >> lane);
                 }
             }
         }
-        __syncthreads();
         // F^T tile [MP x 16 rows] = W1 relu(U)^T, this wave's share of the k range; lane (g, c)
         // ends with F^T[16I + 4g + r][row c]; k-step (jg, q) uses k = 16 jg + 4g + q in group g
         v4f fa[NI];
@@ -123,29 +176,41 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
 #pragma unroll
         for (int I = 0; I < NI; ++I) red[(wv * NI + I) * 64 + lane] = fa[I];
         __syncthreads();
-        if (wv == 0) {
-            const long row = row0 + c;
-            const bool rok = row < total && (!active || active[row / T]);
+        // four latents i0..i0+3 of row rc per thread: the four waves' partial sums of that
+        // group are one 16-byte LDS entry each
+        if (tid < NT4) {
+            const int I = i0 / 16, gg = (i0 % 16) / 4;
+            const long row = row0 + rc;
+            const bool rok = rowok[rc] && i0 < M;
             if (rok) {
-                const float *zc = cur_iter(zbuf, zalt, zsel, (int)(row / T));
+                v4f sum = red[I * 64 + 16 * gg + rc];
 #pragma unroll
-                for (int I = 0; I < NI; ++I) {
-                    v4f sum = red[I * 64 + lane];
+                for (int w = 1; w < 4; ++w) {
+                    const v4f o = red[(w * NI + I) * 64 + 16 * gg + rc];
+                    sum[0] += o[0]; sum[1] += o[1]; sum[2] += o[2]; sum[3] += o[3];
+                }
+                float Fv[4], rv[4];
 #pragma unroll
-                    for (int w = 1; w < 4; ++w) {
-                        const v4f o = red[(w * NI + I) * 64 + lane];
-                        sum[0] += o[0]; sum[1] += o[1]; sum[2] += o[2]; sum[3] += o[3];
+                for (int r = 0; r < 4; ++r) {
+                    const int i = i0 + r;
+                    Fv[r] = 0.f;
+                    rv[r] = 0.f;
+                    if (i < M) {
+                        Fv[r] = fmaf(a.A[i], zT[i * TT + rc], sum[r]) + (a.h1 ? a.h1[i] : 0.f);
+                        rv[r] = cz[r] - Fv[r];
                     }
+                }
+                const size_t e2 = (size_t)row * M + i0;
+                if ((M & 3) == 0) {
+                    if (F_out) *reinterpret_cast<float4 *>(F_out + e2) = make_float4(Fv[0], Fv[1], Fv[2], Fv[3]);
+                    if (r_out) *reinterpret_cast<float4 *>(r_out + e2) = make_float4(rv[0], rv[1], rv[2], rv[3]);
+                } else {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int i = 16 * I + 4 * g + r;
-                        if (i < M) {
-                            const float F = fmaf(a.A[i], zt[c * MP + i], sum[r]) + (a.h1 ? a.h1[i] : 0.f);
-                            const size_t e2 = (size_t)row * M + i;
-                            if (F_out) F_out[e2] = F;
-                            if (r_out) r_out[e2] = zc[e2] - F;
+                    for (int r = 0; r < 4; ++r)
+                        if (i0 + r < M) {
+                            if (F_out) F_out[e2 + r] = Fv[r];
+                            if (r_out) r_out[e2 + r] = rv[r];
                         }
-                    }
                 }
             }
         }

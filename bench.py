@@ -41,14 +41,15 @@ def _plrnn_step(D, model, xd, c, ws_s, ws_a):
                        ws=ws_s, check=False)
     if res["status"] != 0:
         raise RuntimeError(f"deer_solve returned status {res['status']}: {D.load().deer_last_error()}")
-    D.deer_adjoint(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a)
+    # the step's outputs are the parameter gradients: the adjoint itself is not stored
+    D.deer_adjoint(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a, want_lam=False)
     return sum(res["iters"])
 
 
 def _diag_step(D, model, readout, xd, c, ws_s, ws_r, ws_a, bufs):
     res = D.deer_solve(model, xd, 0.0, 0, ws=ws_s, z=bufs["h"])
     r = D.deer_readout_loss(readout, res["z"], xd, g=bufs["g"], ws=ws_r)
-    D.deer_adjoint(model, xd, res["z"], 0.0, 0, g=r["g"], ws=ws_a)
+    D.deer_adjoint(model, xd, res["z"], 0.0, 0, g=r["g"], ws=ws_a, want_lam=False)
     return c.B
 
 
@@ -67,9 +68,9 @@ def kernel_work(c, steps, updates):
         return {
             # forward: b formed from x on the fly; the write pass stores y (8 B per element)
             "k_diag_seg_write": ("hbm", elems * 8 + xin),
-            # adjoint: real cotangent (4 B) and forward states (8 B) read, adjoint written (8 B),
-            # dlam / dBc accumulated on the way
-            "k_diag_scan_lb_grads": ("hbm", elems * 20 + xin),
+            # adjoint: real cotangent (4 B) and forward states (8 B) read, dlam / dBc accumulated
+            # on the way (the training step does not store the adjoint itself)
+            "k_diag_scan_lb_grads": ("hbm", elems * 12 + xin),
             "k_diag_scan_lb": ("hbm", elems * 12 + xin),
             # read-out: three [rows x 64] x [64 x 128] products (s, g, dWa) on the matrix cores
             "k_readout": ("mfma", steps * B * T * 3 * 2.0 * M * c.params["Wa"].shape[0]),

@@ -158,6 +158,13 @@ static int chunk_override() {
     return e ? atoi(e) : 0;
 }
 
+// DEER_GROUP_MAPS=1 / 0 forces the M <= 16 group maps on (where 32 divides the chunk count) or
+// off, whatever the chain count (a tuning and test override)
+static int group_maps_override() {
+    const char *e = getenv("DEER_GROUP_MAPS");
+    return e ? atoi(e) : -1;
+}
+
 // Chunk length of the dense scans: enough chains to fill the machine (about 2048 waves),
 // and a bounded number of chunks per sequence so that the two-level carry pass stays short
 // (1024 for MP <= 32, 512 for MP = 64, whose group pass composes 64 x 64 maps).
@@ -217,6 +224,7 @@ struct PlrnnWs {
     float *r;
     uint32_t *masks;
     float *P, *v, *carry, *gws;
+    float *gmap;   // M <= 16, 32 | chunks: group maps [B][chunks / 32][16 x 16 + 16]
     NewtonCtl ctl;
     float *gpart;
     double *gpart2;
@@ -236,6 +244,11 @@ static PlrnnWs carve_plrnn(void *ws, int B, int T, int M, int op, size_t *bytes)
     w.v = c.take<float>(nch * w.MP);
     w.carry = c.take<float>(nch * w.MP);
     w.gws = c.take<float>(carry_ws_floats(w.MP, B, w.ncs));
+    // group maps once there are at least 64 blocks of 32 chunks (fewer leave the machine idle
+    // while a block composes its maps; the carry kernel is then cheaper)
+    const int gov = group_maps_override();
+    const bool gm = w.MP == 16 && w.ncs % 32 == 0 && (gov < 0 ? nch >= 2048 : gov > 0);
+    w.gmap = gm ? c.take<float>((size_t)B * (w.ncs / 32) * 272) : nullptr;
     if (op == DEER_OP_SOLVE) {
         w.ctl = carve_ctl(c, B, (size_t)T * M, nch);
         w.r = c.take<float>((size_t)B * T * M);
@@ -522,14 +535,20 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
         int r;
         // M <= 16: each wave's four chunks are composed in the forward pass, one kernel walks
         // the composed maps, and the fix-up applies the per-chunk prefix maps
-        const bool wm = w.MP == 16 && w.ncs % 4 == 0;
-        if ((r = launch_newton_product_plrnn(a, zb, za, zsel, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, wm, st)))
+        // 32 | chunks: the forward pass also composes each block's eight wave maps into a
+        // group map and the fix-up walks the group maps itself (no carry kernel)
+        const bool wm = w.MP == 16 && w.ncs % 4 == 0, gm = w.gmap != nullptr;
+        const int mode = gm ? 2 : (wm ? 1 : 0);
+        if ((r = launch_newton_product_plrnn(a, zb, za, zsel, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, mode,
+                                             w.gmap, st)))
             return r;
-        if (wm) r = launch_carry_walk16(false, w.P, w.v, w.carry, dact, B, w.ncs, st);
+        if (gm) r = 0;
+        else if (wm) r = launch_carry_walk16(false, w.P, w.v, w.carry, dact, B, w.ncs, st);
         else r = launch_carry(w.MP, false, w.P, w.v, w.carry, dact, nullptr, B, w.ncs, w.gws, st);
         if (r) return r;
         return launch_fixup_fwd_plrnn(a, w.masks, w.r, w.carry, zb, za, zsel, w.ctl.chain_bits, dact, gam, w.C, w.ncs,
-                                      wm ? w.P : nullptr, wm ? w.v : nullptr, (ctl.fused && dact) ? &fc : nullptr, st);
+                                      wm ? w.P : nullptr, wm ? w.v : nullptr, w.gmap,
+                                      (ctl.fused && dact) ? &fc : nullptr, st);
     };
     if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ncs, ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {

@@ -515,6 +515,23 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
     if (uok0) vout[(size_t)uid * MP + ui] = u;
 }
 
+// A-operand fragments of a 16 x 16 map (P_c, or its transpose) and the vector v_c for the
+// matrix-core carries: lane (g, c) takes row c, columns 4g..4g+3 (transposed: rows 4g..4g+3 of
+// column c) and v_c[4g..4g+3]
+template <bool REV>
+__device__ __forceinline__ void carry16_fetch(const float *__restrict__ Pc, const float *__restrict__ vc, int g, int c,
+                                              float (&a)[4], float (&vv)[4]) {
+    if (!REV) {
+        const float4 t = *reinterpret_cast<const float4 *>(Pc + c * 16 + 4 * g);
+        a[0] = t.x; a[1] = t.y; a[2] = t.z; a[3] = t.w;
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) a[q] = Pc[(4 * g + q) * 16 + c];
+    }
+    const float4 u = *reinterpret_cast<const float4 *>(vc + 4 * g);
+    vv[0] = u.x; vv[1] = u.y; vv[2] = u.z; vv[3] = u.w;
+}
+
 // ---------------------------------------------------------------------------------------
 // M <= 16: register-tiled forward Newton pass and fix-up.
 // A wave holds four chains, one per 16-lane row (lane = 16 * chain + latent), so a row of the
@@ -660,16 +677,19 @@ __device__ __forceinline__ v4f mfma_step16(const v4f &acc, uint32_t wn, int g, c
     return nx;
 }
 
-template <int TB>
-__global__ __launch_bounds__(64) void k_newton_product_plrnn16(
+// WPB waves per block (1, or 8 for the group maps: the block's 32 chunks then belong to one
+// sequence); wmaps: 0 plain chunk aggregates, 1 wave maps, 2 wave maps composed per block into
+// group maps (gmap).
+template <int TB, int WPB>
+__global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
     const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
     const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
     const int *__restrict__ zsel, float *__restrict__ Pout,
     float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
-    int ncs, int wmaps) {
-    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    int ncs, int wmaps, float *__restrict__ gmap) {
+    const int lane = threadIdx.x & 63, wvb = WPB > 1 ? (int)(threadIdx.x >> 6) : 0, g = lane >> 4, c = lane & 15;
     const int nchains = B * ncs;
-    const int chain0 = blockIdx.x * 4;
+    const int chain0 = (blockIdx.x * WPB + wvb) * 4;
     const Chains16 w = chains16(chain0, nchains, ncs, C, T, active, gamma, zsel);
     if (w.maxlen == 0) return;
     float WpD[4], Dq[4];
@@ -802,22 +822,22 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
         //   slot chain0 + n:  prefix    R_n = P_{n-1} ... P_0, s_n = the walk of the first n chunks
         // so that carry(chain0 + n) = R_n carry(chain0) + s_n.  A chunk product in accumulator
         // layout is transposed through LDS into the A-operand layout; vectors ride in column 0.
-        __shared__ float lt[4][16][17];
-        __shared__ float lv[4][16];
+        __shared__ float lt[WPB][3][16][17];
+        __shared__ float lv[WPB][4][16];
 #pragma unroll
-        for (int n = 0; n < 4; ++n)
+        for (int n = 1; n < 4; ++n)
 #pragma unroll
-            for (int r2 = 0; r2 < 4; ++r2) lt[n][4 * g + r2][c] = acc[n][r2];
-        lv[g][c] = u;
+            for (int r2 = 0; r2 < 4; ++r2) lt[wvb][n - 1][4 * g + r2][c] = acc[n][r2];
+        lv[wvb][g][c] = u;
         lds_barrier();
         float Am[3][4];
         v4f bv[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
 #pragma unroll
-            for (int n = 1; n < 4; ++n) Am[n - 1][q] = lt[n][c][4 * g + q];
+            for (int n = 1; n < 4; ++n) Am[n - 1][q] = lt[wvb][n - 1][c][4 * g + q];
 #pragma unroll
-            for (int n = 0; n < 4; ++n) bv[n][q] = c == 0 ? lv[n][4 * g + q] : 0.f;
+            for (int n = 0; n < 4; ++n) bv[n][q] = c == 0 ? lv[wvb][n][4 * g + q] : 0.f;
         }
         v4f R2 = {0.f, 0.f, 0.f, 0.f}, R3 = {0.f, 0.f, 0.f, 0.f}, Qw = {0.f, 0.f, 0.f, 0.f};
         v4f s2 = bv[1], s3 = bv[2], uw = bv[3];
@@ -838,13 +858,56 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn16(
         }
         const v4f outm[4] = {Qw, acc[0], R2, R3}, outv[4] = {uw, bv[0], s2, s3};
 #pragma unroll
-        for (int n = 0; n < 4; ++n) {
+        for (int n = (WPB > 1 ? 1 : 0); n < 4; ++n) {
             float *P = Pout + (size_t)(chain0 + n) * 256;
 #pragma unroll
             for (int r2 = 0; r2 < 4; ++r2) P[(4 * g + r2) * 16 + c] = outm[n][r2];
             if (c == 0)
                 *reinterpret_cast<float4 *>(vout + (size_t)(chain0 + n) * 16 + 4 * g) =
                     make_float4(outv[n][0], outv[n][1], outv[n][2], outv[n][3]);
+        }
+        if (WPB > 1) {
+            // group maps: wave 0 composes the block's eight wave maps in order; slot chain0 of
+            // wave k receives the composition of waves 0..k-1 (carry(wave k) = G_k carry(group)
+            // + g_k), and gmap[b][group] the whole group's map
+            __shared__ float lq[WPB][16][17];
+            __shared__ float lu[WPB][16];
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) lq[wvb][4 * g + r2][c] = Qw[r2];
+            if (c == 0) {
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) lu[wvb][4 * g + r2] = uw[r2];
+            }
+            __syncthreads();
+            if (wvb != 0) return;
+            const int bc0 = blockIdx.x * WPB * 4;   // the block's first chain
+            v4f Gm, gu = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) Gm[r2] = (4 * g + r2 == c) ? 1.f : 0.f;
+            for (int k = 0; k < WPB; ++k) {
+                float *P = Pout + (size_t)(bc0 + 4 * k) * 256;
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) P[(4 * g + r2) * 16 + c] = Gm[r2];
+                if (c == 0)
+                    *reinterpret_cast<float4 *>(vout + (size_t)(bc0 + 4 * k) * 16 + 4 * g) =
+                        make_float4(gu[0], gu[1], gu[2], gu[3]);
+                v4f ng = {0.f, 0.f, 0.f, 0.f}, nu;
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) nu[r2] = c == 0 ? lu[k][4 * g + r2] : 0.f;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float aq = lq[k][c][4 * g + q];
+                    ng = mfma16x16x4(aq, Gm[q], ng);
+                    nu = mfma16x16x4(aq, gu[q], nu);
+                }
+                Gm = ng;
+                gu = nu;
+            }
+            const int ngm = ncs / (4 * WPB);
+            float *Gp = gmap + ((size_t)(bc0 / ncs) * ngm + (bc0 % ncs) / (4 * WPB)) * 272;
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) Gp[(4 * g + r2) * 16 + c] = Gm[r2];
+            if (c == 0) *reinterpret_cast<float4 *>(Gp + 256 + 4 * g) = make_float4(gu[0], gu[1], gu[2], gu[3]);
         }
         return;
     }
@@ -928,7 +991,8 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
                                                           const int *__restrict__ active,
                                                           const float *__restrict__ gamma, int B, int T, int M, int C,
                                                           int ncs, const float *__restrict__ Pm,
-                                                          const float *__restrict__ vmap, FusedCtl fc) {
+                                                          const float *__restrict__ vmap,
+                                                          const float *__restrict__ gmap, FusedCtl fc) {
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int nchains = B * ncs;
     const int chain0 = blockIdx.x * 4;
@@ -957,12 +1021,61 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
     const float Ai = lat ? A[c] : 0.f, hi = (lat && h) ? h[c] : 0.f;
     const float pi = p_of(c, N, alpha), d = Ai * pi;
     float D = 0.f;
+    // group maps: the wave's carry is walked here from the sequence start over the group maps
+    // before the wave's group (four MFMAs a step, maps eight steps ahead), then taken through
+    // the wave's prefix in its group (slot chain0)
+    __shared__ float wcs[16];
+    if (gmap) {
+        const int ngm = ncs / 32, grp = (chain0 % ncs) / 32, bq = chain0 / ncs;
+        const float *Gb = gmap + (size_t)bq * ngm * 272;
+        v4f cur = {0.f, 0.f, 0.f, 0.f};
+        constexpr int PF = 8;
+        float ga[PF][4], gv[PF][4];
+        if (grp > 0) {
+#pragma unroll
+            for (int d2 = 0; d2 < PF; ++d2) {
+                const float *Gk = Gb + (size_t)min(d2, grp - 1) * 272;
+                carry16_fetch<false>(Gk, Gk + 256, g, c, ga[d2], gv[d2]);
+            }
+        }
+        for (int k0 = 0; k0 < grp; k0 += PF) {
+#pragma unroll
+            for (int d2 = 0; d2 < PF; ++d2) {
+                if (k0 + d2 >= grp) break;
+                v4f nx = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) nx = mfma16x16x4(ga[d2][q], cur[q], nx);
+                if (c == 0) {
+#pragma unroll
+                    for (int r2 = 0; r2 < 4; ++r2) nx[r2] += gv[d2][r2];
+                }
+                cur = nx;
+                const float *Gk = Gb + (size_t)min(k0 + d2 + PF, grp - 1) * 272;
+                carry16_fetch<false>(Gk, Gk + 256, g, c, ga[d2], gv[d2]);
+            }
+        }
+        {
+            float wa[4], wvv[4];
+            carry16_fetch<false>(Pm + (size_t)chain0 * 256, vmap + (size_t)chain0 * 16, g, c, wa, wvv);
+            v4f nx = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) nx = mfma16x16x4(wa[q], cur[q], nx);
+            if (c == 0) {
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) wcs[4 * g + r2] = nx[r2] + wvv[r2];
+            }
+        }
+        lds_barrier();
+    }
     if (len > 0 && lat) {
-        if (!Pm || g == 0) {
+        if (!Pm || (g == 0 && !gmap)) {
             D = carry_in[(size_t)id * 16 + c];
+        } else if (g == 0) {
+            D = wcs[c];
         } else {   // composed wave maps: carry = R_g carry(chain0) + s_g
             const float4 *R4 = reinterpret_cast<const float4 *>(Pm + (size_t)id * 256 + c * 16);
-            const float4 *w4 = reinterpret_cast<const float4 *>(carry_in + (size_t)chain0 * 16);
+            const float4 *w4 = gmap ? reinterpret_cast<const float4 *>(wcs)
+                                    : reinterpret_cast<const float4 *>(carry_in + (size_t)chain0 * 16);
             float a0 = vmap[(size_t)id * 16 + c], a1 = 0.f;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
@@ -1400,19 +1513,6 @@ __global__ __launch_bounds__(256) void k_carry_group(const float *__restrict__ P
 // operand, whose accumulator layout is again the next step's B operand, so a step is four
 // dependent MFMAs and no LDS.  The maps of the next PF steps are in flight while a step runs.
 // ---------------------------------------------------------------------------------------
-template <bool REV>
-__device__ __forceinline__ void carry16_fetch(const float *__restrict__ Pc, const float *__restrict__ vc, int g, int c,
-                                              float (&a)[4], float (&vv)[4]) {
-    if (!REV) {
-        const float4 t = *reinterpret_cast<const float4 *>(Pc + c * 16 + 4 * g);
-        a[0] = t.x; a[1] = t.y; a[2] = t.z; a[3] = t.w;
-    } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) a[q] = Pc[(4 * g + q) * 16 + c];
-    }
-    const float4 u = *reinterpret_cast<const float4 *>(vc + 4 * g);
-    vv[0] = u.x; vv[1] = u.y; vv[2] = u.z; vv[3] = u.w;
-}
 
 // walk of the vector: carry_in[c(k)] = cur_k, cur_{k+1} = A_k cur_k + v_{c(k)} (see k_carry)
 template <bool REV>
@@ -2396,11 +2496,13 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
 
 int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
                                 uint32_t *masks, float *P, float *v, const int *active, const float *gamma, int C,
-                                int ncs, bool wmaps, hipStream_t st) {
+                                int ncs, int wmaps, float *gmap, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt("k_newton_product_plrnn", st);
+    if (wmaps == 2 && (MP != 16 || ncs % 32 || !gmap))
+        return invalid_arg("group maps need M <= 16, a chunk count divisible by 32 and their buffer");
 #define NP(MPV)                                                                                                   \
     hipLaunchKernelGGL(k_newton_product_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, \
                        a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs)
@@ -2410,12 +2512,15 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
         hipLaunchKernelGGL(k_newton_product_plrnn64u, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0,
                            z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
     } else if (MP == 16) {
-        if (C % 32)
-            hipLaunchKernelGGL(k_newton_product_plrnn16<16>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
-                               a.x, a.z0, z, zalt, zsel, P, v, active, gamma, a.B, a.T, a.M, C, ncs, (int)wmaps);
-        else
-            hipLaunchKernelGGL(k_newton_product_plrnn16<32>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
-                               a.x, a.z0, z, zalt, zsel, P, v, active, gamma, a.B, a.T, a.M, C, ncs, (int)wmaps);
+#define NP16(TBV, WPBV)                                                                                                \
+    hipLaunchKernelGGL((k_newton_product_plrnn16<TBV, WPBV>), dim3(grid / WPBV), dim3(64 * WPBV), 0, st, a.A, a.W, a.h, \
+                       a.alpha, a.N, a.x, a.z0, z, zalt, zsel, P, v, active, gamma, a.B, a.T, a.M, C, ncs, wmaps, gmap)
+        if (wmaps == 2) {
+            if (C % 32) NP16(16, 8); else NP16(32, 8);
+        } else {
+            if (C % 32) NP16(16, 1); else NP16(32, 1);
+        }
+#undef NP16
     } else if (MP == 32) NP(32); else NP(64);
 #undef NP
     DEER_LAUNCH_CHECK("k_newton_product_plrnn");
@@ -2503,7 +2608,7 @@ int launch_carry_walk16(bool rev, const float *P, const float *v, float *carry, 
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
                            float *z, float *zalt, const int *zsel, uint32_t *chain_bits, const int *active,
                            const float *gamma, int C, int ncs, const float *Pm, const float *vm,
-                           const FusedCtl *fc, hipStream_t st) {
+                           const float *gmap, const FusedCtl *fc, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
@@ -2513,7 +2618,8 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
                        z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
 #define FX16(TBV)                                                                                                 \
     hipLaunchKernelGGL(k_fixup_fwd_plrnn16<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, \
-                       carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs, Pm, vm, fcv)
+                       carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs, Pm, vm, gmap, fcv)
+    if (gmap && (!Pm || ncs % 32)) return invalid_arg("group maps need the wave maps and 32 | chunk count");
     if (Pm && (MP != 16 || ncs % 4))
         return invalid_arg("composed wave maps need M <= 16 and a chunk count divisible by 4");
     if (fc && MP != 16) return invalid_arg("the fused pass-end control needs M <= 16");

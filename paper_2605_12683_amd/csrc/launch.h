@@ -32,7 +32,7 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
                                hipStream_t st);
 int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
                                 uint32_t *masks, float *P, float *v, const int *active, const float *gamma, int C,
-                                int ncs, bool wmaps, hipStream_t st);
+                                int ncs, int wmaps, float *gmap, hipStream_t st);
 // M <= 16 with wave maps (P, v from launch_newton_product_plrnn with wmaps): carries of the
 // wave maps, written to the carry slot of each wave's first chunk
 int launch_carry_walk16(bool rev, const float *P, const float *v, float *carry, const int *active, int B, int ncs,
@@ -47,7 +47,7 @@ size_t carry_ws_floats(int MP, int B, int ncs);
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
                            float *z, float *zalt, const int *zsel, uint32_t *chain_bits, const int *active,
                            const float *gamma, int C, int ncs, const float *Pm, const float *vm,
-                           const FusedCtl *fc, hipStream_t st);
+                           const float *gmap, const FusedCtl *fc, hipStream_t st);
 // device-side Newton control (one entry per sequence)
 struct NewtonDev {
     int *act;       // active flag (read by every kernel of a pass)

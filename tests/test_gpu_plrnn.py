@@ -25,9 +25,11 @@ TOL = 1e-4
 
 @pytest.fixture(autouse=True)
 def _no_chunk_override():
-    os.environ.pop("DEER_CHUNK", None)
+    for k in ("DEER_CHUNK", "DEER_GROUP_MAPS"):
+        os.environ.pop(k, None)
     yield
-    os.environ.pop("DEER_CHUNK", None)
+    for k in ("DEER_CHUNK", "DEER_GROUP_MAPS"):
+        os.environ.pop(k, None)
 
 
 def _case(M, N, B, T, alpha, seed, w_std=None):
@@ -73,11 +75,14 @@ def test_config1_fixed_five_iterations():
     (64, 64, 3, 1000, 0.05, 128), (5, 2, 4, 64, 0.5, 64), (16, 16, 1, 1, 0.2, 0), (8, 8, 2, 2, 0.2, 0),
     # chunk counts divisible by 4 (composed wave maps for M <= 16): full tiles, a ragged second
     # tile, and chunks shorter than a tile
-    (16, 3, 2, 512, 0.2, 16), (7, 3, 3, 640, 0.3, 40), (16, 3, 2, 1000, 0.2, 25)])
+    (16, 3, 2, 512, 0.2, 16), (7, 3, 3, 640, 0.3, 40), (16, 3, 2, 1000, 0.2, 25),
+    # chunk counts divisible by 32 (group maps walked by the fix-up): one, two and four groups
+    (5, 2, 3, 1024, 0.3, 16), (16, 3, 2, 2048, 0.2, 16), (12, 4, 2, 4096, 0.2, 32)])
 def test_solve_reaches_rollout(M, N, B, T, alpha, chunk):
     """Converged GTF-DEER equals the sequential GTF rollout (unique zero of the residual)."""
     if chunk:
         os.environ["DEER_CHUNK"] = str(chunk)
+    os.environ["DEER_GROUP_MAPS"] = "1"   # where 32 divides the chunk count, whatever the size
     c = _case(M, N, B, T, alpha, 200 + M + T)
     m = oracle_model(c)
     say("deer_solve", M, N, B, T, alpha, chunk)
@@ -97,7 +102,7 @@ def test_solve_reaches_rollout(M, N, B, T, alpha, chunk):
 
 @pytest.mark.parametrize("M,N,B,T,alpha,chunk,bound", [(16, 3, 4, 300, 0.2, 0, 0.05), (16, 3, 3, 300, 0.2, 16, 0.3),
                                                        (32, 8, 3, 300, 0.1, 16, 0.1), (64, 64, 2, 200, 0.05, 0, 0.1),
-                                                       (5, 2, 5, 120, 0.3, 7, 0.02)])
+                                                       (5, 2, 5, 120, 0.3, 7, 0.02), (16, 3, 3, 512, 0.2, 16, 0.3)])
 def test_safeguard_rejections_reach_rollout(M, N, B, T, alpha, chunk, bound):
     """A small step bound makes the solver reject updates and retry them damped (the scan
     uses gamma J~ with gamma < 1, down to the fixed-point step); the iterates alternate
@@ -105,6 +110,7 @@ def test_safeguard_rejections_reach_rollout(M, N, B, T, alpha, chunk, bound):
     more passes than plain Newton's show that the safeguard ran."""
     if chunk:
         os.environ["DEER_CHUNK"] = str(chunk)
+    os.environ["DEER_GROUP_MAPS"] = "1"
     c = _case(M, N, B, T, alpha, 600 + M + T)
     m = oracle_model(c)
     say("deer_solve safeguard", M, N, B, T, alpha, chunk, bound)

@@ -88,13 +88,34 @@ void timing_mark(const char *name, hipStream_t st, bool start) {
 }
 
 // ---- small utility kernels -------------------------------------------------------------
+// z_s = [x_{s+1}; 0] for every (b, s): one sequence per blockIdx.y, four consecutive elements of
+// a sequence per thread (a 16-byte store when M is a multiple of 4)
 __global__ void k_fill_teacher(int B, int T, int M, int N, const float *__restrict__ x, float *__restrict__ z) {
-    const size_t n = (size_t)B * T * M;
-    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n; e += (size_t)gridDim.x * blockDim.x) {
-        const int i = (int)(e % M);
-        const size_t bt = e / M;
-        const int b = (int)(bt / T), s = (int)(bt % T);
-        z[e] = i < N ? x[((size_t)b * (T + 1) + s + 1) * N + i] : 0.f;
+    const int b = blockIdx.y;
+    const size_t n = (size_t)T * M;
+    float *zb = z + (size_t)b * n;
+    const float *xb = x + ((size_t)b * (T + 1) + 1) * N;   // row s + 1 of x for row s of z
+    const size_t n4 = (n + 3) / 4;
+    for (size_t e4 = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e4 < n4; e4 += (size_t)gridDim.x * blockDim.x) {
+        const size_t e = 4 * e4;
+        float v[4];
+        size_t s = e / M;
+        int i = (int)(e - s * M);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            v[k] = (e + k < n && i < N) ? xb[s * N + i] : 0.f;
+            if (++i == M) {
+                i = 0;
+                ++s;
+            }
+        }
+        if ((M & 3) == 0) {
+            *reinterpret_cast<float4 *>(zb + e) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                if (e + k < n) zb[e + k] = v[k];
+        }
     }
 }
 __global__ void k_fill_i32(int *p, int n, int v) {
@@ -122,9 +143,10 @@ __global__ void k_fill_f32(float *p, size_t n, float v) {
 }
 
 int launch_fill_teacher(int B, int T, int M, int N, const float *x, float *z, hipStream_t st) {
-    const size_t n = (size_t)B * T * M;
-    const int grid = (int)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
-    hipLaunchKernelGGL(k_fill_teacher, dim3(grid), dim3(256), 0, st, B, T, M, N, x, z);
+    const size_t n4 = ((size_t)T * M + 3) / 4;
+    const size_t want = (n4 + 255) / 256;
+    const int gx = (int)(want < 1024 ? want : 1024);
+    hipLaunchKernelGGL(k_fill_teacher, dim3(gx, B), dim3(256), 0, st, B, T, M, N, x, z);
     DEER_LAUNCH_CHECK("k_fill_teacher");
     return DEER_OK;
 }

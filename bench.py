@@ -82,8 +82,15 @@ def kernel_work(c, steps, updates):
         out["k_newton_product_plrnn"] = ("mfma", fwd * 2.0 * M ** 3)
         out["k_chunk_product_plrnn"] = ("mfma", steps * B * (T - 1) * 2.0 * M ** 3)
         out["k_resjac_plrnn"] = ("hbm", adj * (4 * M + 4 * N + 4 * W))
-        out["k_fixup_fwd_plrnn"] = ("hbm", fwd * (12 * M + 4 * W))
-        out["k_fixup_rev_plrnn"] = ("hbm", adj * (8 * M + 4 * N + 4 * W))
+        if M <= 16:
+            # the register-tiled fix-ups form the residual and the masks again from z and x:
+            # forward z, x read and the next iterate written; reverse z, x read (the training
+            # step keeps the parameter gradients only, so the adjoint is not written)
+            out["k_fixup_fwd_plrnn"] = ("hbm", fwd * (8 * M + 4 * N))
+            out["k_fixup_rev_plrnn"] = ("hbm", adj * (4 * M + 4 * N))
+        else:
+            out["k_fixup_fwd_plrnn"] = ("hbm", fwd * (12 * M + 4 * W))
+            out["k_fixup_rev_plrnn"] = ("hbm", adj * (8 * M + 4 * N + 4 * W))
     else:
         L = c.L
         LW = (L + 31) // 32

@@ -126,8 +126,14 @@ size_t deer_workspace_bytes(const deer_model *model, int B, int T, int op);
  *                counting the verifying one (a sequence converged after k updates reports k).
  *   final_norm   host [B] out or NULL: max |Delta z| of each sequence's last update.
  * Each Newton update is applied before the test; a sequence whose update is below tol
- * is frozen while the others continue.  With fixed_iters == 0 the call synchronises
- * `stream` once per iteration (one device-to-host copy of 2B words) and safeguards the
+ * is frozen while the others continue.  With fixed_iters == 0 the test runs on the device
+ * after every update; a sequence that stops clears a flag in a pinned host block of the
+ * calling thread (allocated on first use, grown with B, kept until the process ends) that
+ * also receives its update count, last norm and status.  The host keeps passes queued ahead
+ * of the device and returns once every sequence has stopped (then without a stream
+ * synchronisation: z is complete in stream order, and the passes still queued skip every
+ * sequence) or at max_iter (after a synchronisation).  Calls from one host thread run one
+ * at a time.  The loop also safeguards the
  * iteration: an update that is not finite, or whose max|Delta z| exceeds
  * step_bound * (1 + max|z|) of its sequence, is discarded and that sequence retried with
  * the damped linearisation gamma J~ (0 <= gamma < 1; gamma = 0 is the fixed-point step
@@ -135,7 +141,7 @@ size_t deer_workspace_bytes(const deer_model *model, int B, int T, int op);
  * gamma has the same fixed point and the same prefix property (one more leading step exact
  * per update), so the solution is unchanged; only the path to it differs.  With
  * fixed_iters > 0 the updates are plain Newton steps applied unconditionally and the call
- * synchronises once at the end (only if iters/final_norm given).
+ * synchronises once at the end (to read the final norms).
  * Returns DEER_OK, DEER_ERR_NOT_CONVERGED (z = last accepted iterate), DEER_ERR_NONFINITE
  * (also when the undamped fixed-point step overflows) or an argument / HIP / workspace
  * error. */

@@ -378,44 +378,74 @@ static size_t diag_bytes(int B, int T, int M, int K, int op) {
     return op == DEER_OP_ADJOINT ? diag_adjoint_ws_bytes(B, T, M, K) : diag_scan_ws_bytes(B, T, M);
 }
 
-// Newton loop shared by the PLRNN kinds.  `update(act, gamma, zsel, z, zalt)` queues one
-// Newton update of the sequences whose device flag is set (all, when act is null),
+// Newton loop shared by the PLRNN kinds.  `update(act, gamma, zsel, z, zalt, mark, pass_no)`
+// queues one Newton update of the sequences whose device flag is set (all, when act is null),
 // linearised with the per-sequence factor gamma (gamma J~; null: 1), reading each sequence's
 // iterate from the buffer zsel selects and writing iterate + Delta to the other one (zsel
 // null and zalt == z: in place), and leaves per-chain max|Delta| and max|z| bits in
-// ctl.chain_bits.
+// ctl.chain_bits; with a mark, the pass writes pass_no to it as it starts.
 //
 // With a convergence test (fixed_iters == 0) the test and the update safeguard run on the
-// device after every pass (k_seq_ctl): an update that is not finite, or whose max|Delta|
-// exceeds step_bound (1 + max|z|), is not kept and the sequence is retried with gamma < 1;
-// gamma returns to 1 over accepted updates.  gamma = 1 is the exact Newton step, gamma = 0
-// the fixed-point step z_t <- F(z~_{t-1}); every gamma keeps the fixed point and the prefix
-// property.  The host queues passes in batches and reads the active flags of a batch while
-// the next batch already runs (the pass-end control clears a pinned host copy of the flags
-// too; an event per batch tells the host which passes are complete), so the device does not
-// wait for the host; a sequence frozen inside a batch makes the rest of the queued kernels
-// skip it, and once every sequence is frozen the passes still queued skip everything.
+// device after every pass (in the fix-up, or k_seq_ctl): an update that is not finite, or
+// whose max|Delta| exceeds step_bound (1 + max|z|), is not kept and the sequence is retried
+// with gamma < 1; gamma returns to 1 over accepted updates.  gamma = 1 is the exact Newton
+// step, gamma = 0 the fixed-point step z_t <- F(z~_{t-1}); every gamma keeps the fixed point
+// and the prefix property.  A sequence that stops clears its flag on the device and in a
+// pinned host block that also receives its results, so the host follows the device without
+// copies; a sequence frozen while passes are queued makes them skip it, and once every
+// sequence is frozen the passes still queued skip everything.  The call returns when every
+// sequence has stopped (or at the iteration cap); z is then complete in stream order.
 constexpr float kDefaultStepBound = 1e3f;
 constexpr NewtonDamp kDamp = {1.f / 64, 4.f, 4.f, 1e-4f};
 constexpr int kFirstBatch = 4, kBatch = 1;
 
-// pinned, device-coherent host copy of the active flags (per host thread, grown on demand,
-// kept for the life of the process)
-struct ActPoll {
-    int *host = nullptr;
+// Pinned, device-coherent host block of the Newton loop, one per host thread (grown on
+// demand, kept for the life of the process): act | it | norm | status (cap words each; see
+// NewtonDev), then the pass mark.  Passes are numbered per thread; the M <= 16 forward pass
+// writes its number to the mark as it starts.
+struct HostBlk {
+    int *base = nullptr;
     size_t cap = 0;
+    uint32_t next_pass = 1;   // number of the next marked pass
 };
-static thread_local ActPoll t_poll;
-static int poll_flags(int B, int **flags) {
-    if ((size_t)B > t_poll.cap) {
-        if (t_poll.host) (void)hipHostFree(t_poll.host);
-        t_poll.host = nullptr;
-        t_poll.cap = 0;
-        DEER_HIP(hipHostMalloc((void **)&t_poll.host, (size_t)B * sizeof(int), hipHostMallocCoherent));
-        t_poll.cap = (size_t)B;
+static thread_local HostBlk t_host;
+static int host_block(int B, NewtonDev &nd, uint32_t **mark) {
+    if ((size_t)B > t_host.cap) {
+        if (t_host.base) (void)hipHostFree(t_host.base);
+        t_host.base = nullptr;
+        t_host.cap = 0;
+        DEER_HIP(hipHostMalloc((void **)&t_host.base, (4 * (size_t)B + 32) * sizeof(int), hipHostMallocCoherent));
+        t_host.cap = (size_t)B;
+        // no pass of this thread is pending (every earlier solve returned after its last mark)
+        *(uint32_t *)(t_host.base + 4 * t_host.cap) = t_host.next_pass - 1;
     }
-    *flags = t_poll.host;
+    int *p = t_host.base;
+    const size_t cap = t_host.cap;
+    nd.hact = p;
+    nd.hit = p + cap;
+    nd.hnorm = (float *)(p + 2 * cap);
+    nd.hstat = p + 3 * cap;
+    *mark = (uint32_t *)(p + 4 * cap);
     return DEER_OK;
+}
+
+// Waits until the pass mark has reached `want` (in wrapping order).  The stream is queried now
+// and then, so that a stream that ran dry without the mark is an error, not a hang.
+static int wait_mark(const uint32_t *mark, uint32_t want, hipStream_t st) {
+    auto reached = [&]() { return (int32_t)(__atomic_load_n(mark, __ATOMIC_ACQUIRE) - want) >= 0; };
+    for (unsigned spin = 1;; ++spin) {
+        if (reached()) return DEER_OK;
+        if ((spin & 1023u) == 0u) {
+            const hipError_t e = hipStreamQuery(st);
+            if (e == hipSuccess) {
+                if (reached()) return DEER_OK;
+                set_error("the stream finished without the forward pass's mark");
+                return DEER_ERR_HIP;
+            }
+            if (e != hipErrorNotReady) return hip_fail(e, "hipStreamQuery");
+        }
+        __builtin_ia32_pause();
+    }
 }
 
 template <class Update>
@@ -428,7 +458,7 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
     int rc;
     if (fixed) {
         for (int k = 0; k < fixed; ++k)
-            if ((rc = update(nullptr, nullptr, nullptr, z, z))) return rc;
+            if ((rc = update(nullptr, nullptr, nullptr, z, z, nullptr, 0u))) return rc;
         if ((rc = launch_seq_max(ctl.chain_bits, nullptr, ctl.norm_bits, B, ncs, st))) return rc;
         std::vector<uint32_t> nb(B, 0);
         DEER_HIP(hipMemcpyAsync(nb.data(), ctl.norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
@@ -441,57 +471,69 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
         return DEER_OK;
     }
     NewtonDev nd = ctl.nd;
-    if (!nd.hact && (rc = poll_flags(B, &nd.hact))) return rc;
+    uint32_t *mark = nullptr;
+    if ((rc = host_block(B, nd, &mark))) return rc;
     int *const hact = nd.hact;
     for (int b = 0; b < B; ++b) hact[b] = 1;   // no kernel of this stream that writes it is pending
     if ((rc = launch_ctl_init(nd, ctl.seq, B, st))) return rc;
-    hipEvent_t ev[2] = {nullptr, nullptr};
-    auto done_events = [&]() {
-        for (hipEvent_t &e : ev)
-            if (e) (void)hipEventDestroy(e);
+    auto all_stopped = [&]() {
+        bool any = false;
+        for (int b = 0; b < B; ++b) any |= __atomic_load_n(hact + b, __ATOMIC_ACQUIRE) != 0;
+        return !any;
     };
-    for (hipEvent_t &e : ev) {
-        const hipError_t err = hipEventCreateWithFlags(&e, hipEventDisableTiming);
-        if (err != hipSuccess) {
-            done_events();
-            return hip_fail(err, "hipEventCreateWithFlags");
+    bool stopped = false;
+    if (ctl.fused) {
+        // Short passes (the fused M <= 16 path).  The forward pass of pass p marks its start,
+        // when every earlier pass, and so the decisions of pass p - 1, is complete.  The host
+        // keeps one pass queued ahead: once pass p has started it reads the flags as of pass
+        // p - 1 and queues pass p + 1 (a whole pass of time to do so), so the device does not
+        // wait for the host and one pass runs past convergence (it skips every sequence).
+        // The loop ends only after the mark of the last queued pass, so no mark is pending.
+        int passes = 0;
+        auto queue = [&]() {
+            const int r = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt, mark, t_host.next_pass);
+            ++t_host.next_pass;
+            ++passes;
+            return r;
+        };
+        rc = queue();
+        if (!rc && passes < max_iter) rc = queue();
+        while (!rc) {
+            if ((rc = wait_mark(mark, t_host.next_pass - 1, st))) break;
+            if ((stopped = all_stopped())) break;
+            if (passes >= max_iter) break;
+            rc = queue();
         }
-    }
-    auto check = [&](hipError_t err, const char *what) {
-        if (err == hipSuccess) return 0;
-        done_events();
-        return hip_fail(err, what);
-    };
-    int passes = 0, batch = kFirstBatch, k = 0;
-    while (passes < max_iter) {
-        const int n = batch < max_iter - passes ? batch : max_iter - passes;
-        for (int j = 0; j < n; ++j) {
-            rc = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt);
-            if (!rc && !ctl.fused) rc = launch_seq_ctl(ctl.chain_bits, nd, B, ncs, o->tol, bound, kDamp, st);
-            if (rc) {
-                done_events();
-                return rc;
+        if (rc) return rc;
+    } else {
+        // Long passes: batches of passes with an event after each; the host waits for the batch
+        // just queued (the wait is small next to a pass, and a pass queued past convergence is
+        // not).
+        hipEvent_t ev = nullptr;
+        DEER_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+        int passes = 0, batch = kFirstBatch;
+        while (passes < max_iter) {
+            const int n = batch < max_iter - passes ? batch : max_iter - passes;
+            for (int j = 0; j < n && !rc; ++j) {
+                rc = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt, nullptr, 0u);
+                if (!rc) rc = launch_seq_ctl(ctl.chain_bits, nd, B, ncs, o->tol, bound, kDamp, st);
             }
+            if (rc) break;
+            hipError_t e = hipEventRecord(ev, st);
+            if (e == hipSuccess) e = hipEventSynchronize(ev);
+            if (e != hipSuccess) {
+                rc = hip_fail(e, "hipEventRecord / hipEventSynchronize");
+                break;
+            }
+            passes += n;
+            batch = kBatch;
+            if ((stopped = all_stopped())) break;
         }
-        passes += n;
-        if ((rc = check(hipEventRecord(ev[k & 1], st), "hipEventRecord"))) return rc;
-        batch = kBatch;
-        // Short passes (the fused M <= 16 path): the flags as of the end of the previous batch,
-        // read while this one runs (they only go from 1 to 0, so a later pass having cleared
-        // more is harmless).  Long passes: this batch's flags, as the host wait is then small
-        // next to a pass and a pass queued past convergence is not.
-        const int kc = ctl.fused ? k - 1 : k;
-        if (kc >= 0) {
-            if ((rc = check(hipEventSynchronize(ev[kc & 1]), "hipEventSynchronize"))) return rc;
-            bool any = false;
-            for (int b = 0; b < B; ++b) any |= __atomic_load_n(hact + b, __ATOMIC_ACQUIRE) != 0;
-            if (!any) break;
-        }
-        ++k;
+        (void)hipEventDestroy(ev);
+        if (rc) return rc;
     }
-    done_events();
     // sequences whose iterate ended in the second buffer are copied back on the device (one
-    // launch, no host decision), then the control block is read once
+    // launch, no host decision)
     {
         const size_t n4 = (seq_elems + 3) / 4;
         const unsigned gx = (unsigned)((n4 + 255) / 256 < 256 ? (n4 + 255) / 256 : 256);
@@ -499,6 +541,18 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
                            (const int *)nd.sel, seq_elems);
         DEER_LAUNCH_CHECK("k_copy_sel");
     }
+    if (stopped) {
+        // every sequence has stopped: its results are in the host block, and the kernels still
+        // queued only skip (z is complete in stream order)
+        for (int b = 0; b < B; ++b) {
+            act[b] = 0;
+            it[b] = nd.hit[b];
+            norm[b] = nd.hnorm[b];
+            if (nd.hstat[b] == 2) nonfinite = true;
+        }
+        return DEER_OK;
+    }
+    // iteration cap reached: the control block is read once
     std::vector<uint32_t> h(7 * (size_t)B);
     DEER_HIP(hipMemcpyAsync(h.data(), ctl.blk, h.size() * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
     DEER_HIP(hipStreamSynchronize(st));
@@ -551,9 +605,11 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     // M <= 16: the fix-up also takes the pass-end control of the adaptive loop
     NewtonCtl ctl = w.ctl;
     ctl.fused = w.MP == 16 && o->fixed_iters <= 0;
-    if (ctl.fused && (rc = poll_flags(B, &ctl.nd.hact))) return rc;
+    uint32_t *mark_unused = nullptr;
+    if (ctl.fused && (rc = host_block(B, ctl.nd, &mark_unused))) return rc;
     const FusedCtl fc{ctl.nd, ctl.seq, o->tol, o->step_bound == 0.f ? kDefaultStepBound : o->step_bound, kDamp};
-    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za) -> int {
+    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *mark,
+                      uint32_t pass_no) -> int {
         int r;
         // M <= 16: each wave's four chunks are composed in the forward pass, one kernel walks
         // the composed maps, and the fix-up applies the per-chunk prefix maps
@@ -562,7 +618,7 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
         const bool wm = w.MP == 16 && w.ncs % 4 == 0, gm = w.gmap != nullptr;
         const int mode = gm ? 2 : (wm ? 1 : 0);
         if ((r = launch_newton_product_plrnn(a, zb, za, zsel, w.r, w.masks, w.P, w.v, dact, gam, w.C, w.ncs, mode,
-                                             w.gmap, st)))
+                                             w.gmap, mark, pass_no, st)))
             return r;
         if (gm) r = 0;
         else if (wm) r = launch_carry_walk16(false, w.P, w.v, w.carry, dact, B, w.ncs, st);
@@ -594,7 +650,8 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
     const DenseWs &d = w.d;
-    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za) -> int {
+    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *,
+                      uint32_t) -> int {
         int r;
         if ((r = launch_resjac_shplrnn(a, zb, za, zsel, nullptr, w.r, w.masks, dact, st))) return r;
         if ((r = launch_jacform_shplrnn(a, w.masks, w.J, dact, gam, st))) return r;

@@ -686,8 +686,10 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
     const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
     const int *__restrict__ zsel, float *__restrict__ Pout,
     float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
-    int ncs, int wmaps, float *__restrict__ gmap) {
+    int ncs, int wmaps, float *__restrict__ gmap, uint32_t *mark, uint32_t pass_no) {
     const int lane = threadIdx.x & 63, wvb = WPB > 1 ? (int)(threadIdx.x >> 6) : 0, g = lane >> 4, c = lane & 15;
+    if (mark && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(mark, pass_no, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     const int nchains = B * ncs;
     const int chain0 = (blockIdx.x * WPB + wvb) * 4;
     const Chains16 w = chains16(chain0, nchains, ncs, C, T, active, gamma, zsel);
@@ -934,21 +936,27 @@ __device__ __forceinline__ void seq_decide(int b, uint32_t e, uint32_t zm, const
     const bool fin = e < 0x7f800000u;
     float om = nd.om[b];
     const bool keep = fin && (bound < 0.f || om >= 1.f || ef <= bound * (1.f + zf));
+    // a stopped sequence: device control block, then the host block (act last)
+    auto stop = [&](int it, int status) {
+        nd.act[b] = 0;
+        nd.status[b] = status;
+        if (nd.hact) {
+            nd.hit[b] = it;
+            nd.hnorm[b] = ef;
+            nd.hstat[b] = status;
+            __hip_atomic_store(nd.hact + b, 0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+    };
     if (keep) {
         nd.sel[b] ^= 1;
-        nd.it[b] += 1;
+        const int it = nd.it[b] + 1;
+        nd.it[b] = it;
         nd.norm[b] = ef;
         if (om > 0.f) om = om / dp.shrink < dp.floor ? 0.f : om / dp.shrink;
-        if (ef < tol) {
-            nd.act[b] = 0;
-            if (nd.hact) nd.hact[b] = 0;
-            nd.status[b] = 1;
-        }
+        if (ef < tol) stop(it, 1);
     } else if (om >= 1.f) {
         nd.norm[b] = ef;
-        nd.act[b] = 0;
-        if (nd.hact) nd.hact[b] = 0;
-        nd.status[b] = 2;
+        stop(nd.it[b], 2);
     } else {
         om = om == 0.f ? dp.first : fminf(1.f, om * dp.grow);
     }
@@ -2496,7 +2504,7 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
 
 int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
                                 uint32_t *masks, float *P, float *v, const int *active, const float *gamma, int C,
-                                int ncs, int wmaps, float *gmap, hipStream_t st) {
+                                int ncs, int wmaps, float *gmap, uint32_t *mark, uint32_t pass_no, hipStream_t st) {
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
@@ -2508,13 +2516,15 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
                        a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs)
     if (wmaps && (MP != 16 || ncs % 4))
         return invalid_arg("composed wave maps need M <= 16 and a chunk count divisible by 4");
+    if (mark && MP != 16) return invalid_arg("pass marks are written by the M <= 16 forward pass only");
     if (MP == 64 && (a.N == 0 || a.N == a.M)) {   // uniform forcing factor: W-in-LDS kernel
         hipLaunchKernelGGL(k_newton_product_plrnn64u, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0,
                            z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
     } else if (MP == 16) {
 #define NP16(TBV, WPBV)                                                                                                \
     hipLaunchKernelGGL((k_newton_product_plrnn16<TBV, WPBV>), dim3(grid / WPBV), dim3(64 * WPBV), 0, st, a.A, a.W, a.h, \
-                       a.alpha, a.N, a.x, a.z0, z, zalt, zsel, P, v, active, gamma, a.B, a.T, a.M, C, ncs, wmaps, gmap)
+                       a.alpha, a.N, a.x, a.z0, z, zalt, zsel, P, v, active, gamma, a.B, a.T, a.M, C, ncs, wmaps, gmap, \
+                       mark, pass_no)
         if (wmaps == 2) {
             if (C % 32) NP16(16, 8); else NP16(32, 8);
         } else {

@@ -30,9 +30,11 @@ int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, 
 int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *masks, const float *rhs, const float *z,
                                float seed_scale, float *P, float *v, const int *active, int C, int ncs,
                                hipStream_t st);
+// M <= 16 only: block 0 of the pass writes pass_no to the host-visible word *mark as it
+// starts (every kernel queued before it has completed); mark may be null
 int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
                                 uint32_t *masks, float *P, float *v, const int *active, const float *gamma, int C,
-                                int ncs, int wmaps, float *gmap, hipStream_t st);
+                                int ncs, int wmaps, float *gmap, uint32_t *mark, uint32_t pass_no, hipStream_t st);
 // M <= 16 with wave maps (P, v from launch_newton_product_plrnn with wmaps): carries of the
 // wave maps, written to the carry slot of each wave's first chunk
 int launch_carry_walk16(bool rev, const float *P, const float *v, float *carry, const int *active, int B, int ncs,
@@ -57,7 +59,13 @@ struct NewtonDev {
     int *it;        // accepted updates
     float *norm;    // max |Delta| of the last accepted (or final) update
     int *status;    // 0 running, 1 converged, 2 non-finite
-    int *hact;      // pinned host copy of act, cleared together with act (may be null)
+    // pinned host block (all four may be null): when a sequence stops, its update count,
+    // last max |Delta| and status are written to hit, hnorm, hstat, and then (with release
+    // order at system scope) its entry of hact, set to 1 by the host, is cleared
+    int *hact;
+    int *hit;
+    float *hnorm;
+    int *hstat;
 };
 struct NewtonDamp {
     float first, grow, shrink, floor;

@@ -132,6 +132,27 @@ def test_iteration_counts_match_oracle():
     assert max(abs(a - b) for a, b in zip(res["iters"], ref["iters"].tolist())) <= 1
 
 
+def test_consecutive_solves_share_the_host_block():
+    """Solves in a row on one host thread: the pinned host block (flags, results, pass mark)
+    grows with B and is reused; M <= 16 (passes marked by the forward pass) and M > 16 (an
+    event per batch) alternate.  Each result must be the rollout with oracle-like counts."""
+    for k, (M, N, B, T) in enumerate([(16, 3, 2, 300), (16, 3, 37, 200), (20, 4, 3, 250), (8, 3, 3, 400),
+                                      (16, 3, 64, 128), (5, 2, 1, 90)]):
+        c = _case(M, N, B, T, 0.2, 900 + k)
+        m = oracle_model(c)
+        say("deer_solve in a row", M, N, B, T)
+        res = D.deer_solve(m, c.x, 0.2, N, tol=1e-5, max_iter=100)
+        assert res["status"] == 0, res
+        assert rel_inf(res["z"].cpu().numpy(), O.rollout(m, c.x, 0.2, N)) < TOL
+        ref = O.newton(m, c.x, 0.2, N, tol=1e-5)
+        assert max(abs(a - b) for a, b in zip(res["iters"], ref["iters"].tolist())) <= 1
+        assert all(n < 1e-5 for n in res["norms"])
+    # the iteration cap after a grown block: the control block is read back instead
+    c = _case(16, 3, 2, 300, 0.2, 950)
+    res = D.deer_solve(oracle_model(c), c.x, 0.2, 3, tol=1e-5, max_iter=2, check=False)
+    assert res["status"] == 2 and res["iters"] == [2, 2]
+
+
 def test_alpha1_full_observation_two_updates():
     """alpha = 1, M <= N: z* = F(zbar) in closed form; the GPU stops after 2 updates."""
     c = _case(6, 6, 3, 500, 1.0, 11, w_std=0.8)

@@ -591,6 +591,51 @@ __device__ __forceinline__ float row16_dot(const float (&w)[16], float v) {
           "v"(w[9]), "v"(w[10]), "v"(w[11]), "v"(w[12]), "v"(w[13]), "v"(w[14]), "v"(w[15]));
     return a0 + a1;
 }
+
+// two independent row products W v0, W v1 (each summed exactly as row16_dot), interleaved so
+// that dependent multiply-adds are four instructions apart
+__device__ __forceinline__ void row16_dot2(const float (&w)[16], float v0, float v1, float &r0, float &r1) {
+    float a0, a1, b0, b1;
+    asm volatile(
+        "s_nop 1\n"
+        "v_mul_f32_e32 %0, %4, %6\n"
+        "v_mul_f32_e32 %2, %5, %6\n"
+        "v_mul_f32_dpp %1, %4, %7" DEER_RR(1)
+        "v_mul_f32_dpp %3, %5, %7" DEER_RR(1)
+        "v_fmac_f32_dpp %0, %4, %8" DEER_RR(2)
+        "v_fmac_f32_dpp %2, %5, %8" DEER_RR(2)
+        "v_fmac_f32_dpp %1, %4, %9" DEER_RR(3)
+        "v_fmac_f32_dpp %3, %5, %9" DEER_RR(3)
+        "v_fmac_f32_dpp %0, %4, %10" DEER_RR(4)
+        "v_fmac_f32_dpp %2, %5, %10" DEER_RR(4)
+        "v_fmac_f32_dpp %1, %4, %11" DEER_RR(5)
+        "v_fmac_f32_dpp %3, %5, %11" DEER_RR(5)
+        "v_fmac_f32_dpp %0, %4, %12" DEER_RR(6)
+        "v_fmac_f32_dpp %2, %5, %12" DEER_RR(6)
+        "v_fmac_f32_dpp %1, %4, %13" DEER_RR(7)
+        "v_fmac_f32_dpp %3, %5, %13" DEER_RR(7)
+        "v_fmac_f32_dpp %0, %4, %14" DEER_RR(8)
+        "v_fmac_f32_dpp %2, %5, %14" DEER_RR(8)
+        "v_fmac_f32_dpp %1, %4, %15" DEER_RR(9)
+        "v_fmac_f32_dpp %3, %5, %15" DEER_RR(9)
+        "v_fmac_f32_dpp %0, %4, %16" DEER_RR(10)
+        "v_fmac_f32_dpp %2, %5, %16" DEER_RR(10)
+        "v_fmac_f32_dpp %1, %4, %17" DEER_RR(11)
+        "v_fmac_f32_dpp %3, %5, %17" DEER_RR(11)
+        "v_fmac_f32_dpp %0, %4, %18" DEER_RR(12)
+        "v_fmac_f32_dpp %2, %5, %18" DEER_RR(12)
+        "v_fmac_f32_dpp %1, %4, %19" DEER_RR(13)
+        "v_fmac_f32_dpp %3, %5, %19" DEER_RR(13)
+        "v_fmac_f32_dpp %0, %4, %20" DEER_RR(14)
+        "v_fmac_f32_dpp %2, %5, %20" DEER_RR(14)
+        "v_fmac_f32_dpp %1, %4, %21" DEER_RR(15)
+        "v_fmac_f32_dpp %3, %5, %21" DEER_RR(15)
+        : "=&v"(a0), "=&v"(a1), "=&v"(b0), "=&v"(b1)
+        : "v"(v0), "v"(v1), "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "v"(w[4]), "v"(w[5]), "v"(w[6]), "v"(w[7]),
+          "v"(w[8]), "v"(w[9]), "v"(w[10]), "v"(w[11]), "v"(w[12]), "v"(w[13]), "v"(w[14]), "v"(w[15]));
+    r0 = a0 + a1;
+    r1 = b0 + b1;
+}
 #undef DEER_RR
 
 // Buffer resource with a wave-uniform base: an access adds a per-lane byte offset (VGPR) and a
@@ -613,7 +658,9 @@ __device__ __forceinline__ void bstore_u(__amdgpu_buffer_rsrc_t rs, uint32_t v, 
 __device__ __forceinline__ int rfl_i(int v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ float rfl_f(float v) { return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v))); }
 
-// the wave's four chains: lengths, damping, and whether they all read one iterate buffer
+// the wave's four chains: sequence and chunk index, lengths, damping, and whether they all read
+// one iterate buffer.  chain0 is wave-uniform, so every value here is scalar; the control words
+// of the four chains are loaded at once (clamped indices) and combined afterwards.
 struct Chains16 {
     int plen[4];
     float gam[4];
@@ -624,27 +671,56 @@ __device__ __forceinline__ Chains16 chains16(int chain0, int nchains, int ncs, i
                                              const int *__restrict__ active, const float *__restrict__ gamma,
                                              const int *__restrict__ zsel) {
     Chains16 w;
+    const int b0 = chain0 / ncs, c0 = chain0 - b0 * ncs;
+    int act[4], sel[4], bq[4], cq[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        int bb = b0, cc = c0 + n;
+#pragma unroll
+        for (int k = 0; k < 3; ++k)   // c0 + n < c0 + 4 <= 4 ncs
+            if (cc >= ncs) {
+                cc -= ncs;
+                ++bb;
+            }
+        const bool ok = chain0 + n < nchains;
+        bq[n] = ok ? bb : 0;
+        cq[n] = ok ? cc : 0;
+        act[n] = active ? active[bq[n]] : 1;
+        w.gam[n] = gamma ? gamma[bq[n]] : 1.f;
+        sel[n] = zsel ? zsel[bq[n]] : 0;
+    }
     w.minlen = C;
     w.maxlen = 0;
     w.onebuf = true;
     int sel0 = -1;
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
-        const int id = chain0 + n;
-        bool ok = id < nchains;
-        const int b = ok ? id / ncs : 0, cc = ok ? id % ncs : 0;
-        ok = ok && (!active || active[b]);
-        w.plen[n] = rfl_i(ok ? min(C, T - cc * C) : 0);
-        w.gam[n] = rfl_f(gamma ? gamma[b] : 1.f);
-        const int sel = rfl_i(zsel ? zsel[b] : 0);
+        const bool ok = chain0 + n < nchains && act[n] != 0;
+        w.plen[n] = ok ? min(C, T - cq[n] * C) : 0;
         if (w.plen[n] > 0) {
-            if (sel0 >= 0 && sel != sel0) w.onebuf = false;
-            sel0 = sel;
+            if (sel0 >= 0 && sel[n] != sel0) w.onebuf = false;
+            sel0 = sel[n];
         }
         w.minlen = min(w.minlen, w.plen[n]);
         w.maxlen = max(w.maxlen, w.plen[n]);
     }
     return w;
+}
+
+// sequence b and first step s0 of chain chain0 + g (g < 4) without a division (chain0 is
+// uniform); 0, 0 past the last chain
+__device__ __forceinline__ void chain_pos(int chain0, int g, int nchains, int ncs, int C, int &b, int &s0) {
+    const int b0 = chain0 / ncs;
+    int bb = b0, cc = chain0 - b0 * ncs + g;
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        if (cc >= ncs) {
+            cc -= ncs;
+            ++bb;
+        }
+    const bool ok = chain0 + g < nchains;
+    b = ok ? bb : 0;
+    s0 = ok ? cc * C : 0;
 }
 
 // acc[n] *= gamma_n^(steps chain n ran in the tile [t0, t0 + tl)): J~ = gamma (...) per step
@@ -687,13 +763,53 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
     const int *__restrict__ zsel, float *__restrict__ Pout,
     float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
     int ncs, int wmaps, float *__restrict__ gmap, uint32_t *mark, uint32_t pass_no) {
-    const int lane = threadIdx.x & 63, wvb = WPB > 1 ? (int)(threadIdx.x >> 6) : 0, g = lane >> 4, c = lane & 15;
+    // the wave index is uniform: the chain set, its control words and the tile addresses are
+    // scalar values (scalar loads, no per-lane address arithmetic)
+    const int lane = threadIdx.x & 63, wvb = WPB > 1 ? rfl_i((int)(threadIdx.x >> 6)) : 0, g = lane >> 4, c = lane & 15;
     if (mark && blockIdx.x == 0 && threadIdx.x == 0)
         __hip_atomic_store(mark, pass_no, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     const int nchains = B * ncs;
     const int chain0 = (blockIdx.x * WPB + wvb) * 4;
     const Chains16 w = chains16(chain0, nchains, ncs, C, T, active, gamma, zsel);
     if (w.maxlen == 0) return;
+    // row part: this lane is latent c of chain g
+    const int id = chain0 + g;
+    const bool okc = id < nchains;
+    int b, s0;
+    chain_pos(chain0, g, nchains, ncs, C, b, s0);
+    int len = 0;
+    float ugam = 1.f;
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+        if (n == g) {
+            len = w.plen[n];
+            ugam = w.gam[n];
+        }
+    const bool lat = c < M, forced = c < N;
+    // tile resources, based at the first row of the wave's first chain
+    const int b0 = chain0 / ncs, s00 = (chain0 % ncs) * C;
+    const size_t row0 = (size_t)b0 * T + s00, xrow0 = (size_t)b0 * (T + 1) + s00;
+    const uint32_t drow = (uint32_t)((size_t)b * T + s0 - row0), dxrow = (uint32_t)((size_t)b * (T + 1) + s0 - xrow0);
+    const float *zw = cur_iter(zbuf, zalt, zsel, b0);
+    const auto rz = wave_rsrc(zw + row0 * M);
+    const auto rx = wave_rsrc(N > 0 ? x + xrow0 * N : zw);
+    const uint32_t vz = lat ? 4u * (drow * M + c) : kOffLane;
+    const uint32_t vx = forced ? 4u * (dxrow * N + c) : kOffLane;
+    // the first tile's loads go out before the weights are gathered
+    float zv[TB], xv[TB];
+    if (w.onebuf && TB <= w.minlen) {
+#pragma unroll
+        for (int tt = 0; tt < TB; ++tt) {
+            zv[tt] = bload(rz, vz, 4 * tt * M);
+            xv[tt] = bload(rx, vx, 4 * tt * N);
+        }
+    }
+    const float *z = cur_iter(zbuf, zalt, zsel, b);
+    float zprev = 0.f;
+    if (len > 0 && lat) {
+        if (s0 == 0) zprev = z0 ? z0[(size_t)b * M + c] : (forced ? x[(size_t)b * (T + 1) * N + c] : 0.f);
+        else zprev = z[((size_t)b * T + s0 - 1) * M + c];
+    }
     float WpD[4], Dq[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -707,19 +823,6 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
     for (int n = 0; n < 4; ++n)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[n][r] = (4 * g + r == c) ? 1.f : 0.f;
-    // row part: this lane is latent c of chain g
-    const int id = chain0 + g;
-    const bool okc = id < nchains;
-    const int b = okc ? id / ncs : 0, s0 = okc ? (id % ncs) * C : 0;
-    int len = 0;
-    float ugam = 1.f;
-#pragma unroll
-    for (int n = 0; n < 4; ++n)
-        if (n == g) {
-            len = w.plen[n];
-            ugam = w.gam[n];
-        }
-    const bool lat = c < M, forced = c < N;
     int src[16];
     row_sources(c, src);
     float wr[16];
@@ -727,43 +830,33 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
     for (int k = 0; k < 16; ++k) wr[k] = (lat && src[k] < M) ? W[c * M + src[k]] : 0.f;
     const float Ai = lat ? A[c] : 0.f, hi = (lat && h) ? h[c] : 0.f;
     const float pi = p_of(c, N, alpha), di = Ai * pi;
-    const float *z = cur_iter(zbuf, zalt, zsel, b);
-    float zprev = 0.f;
-    if (len > 0 && lat) {
-        if (s0 == 0) zprev = z0 ? z0[(size_t)b * M + c] : (forced ? x[(size_t)b * (T + 1) * N + c] : 0.f);
-        else zprev = z[((size_t)b * T + s0 - 1) * M + c];
-    }
-    // tile resources, based at the first row of the wave's first chain
-    const int b0 = chain0 / ncs, s00 = (chain0 % ncs) * C;
-    const size_t row0 = (size_t)b0 * T + s00, xrow0 = (size_t)b0 * (T + 1) + s00;
-    const uint32_t drow = (uint32_t)((size_t)b * T + s0 - row0), dxrow = (uint32_t)((size_t)b * (T + 1) + s0 - xrow0);
-    const float *zw = cur_iter(zbuf, zalt, zsel, b0);
-    const auto rz = wave_rsrc(zw + row0 * M);
-    const auto rx = wave_rsrc(N > 0 ? x + xrow0 * N : zw);
-    const uint32_t vz = lat ? 4u * (drow * M + c) : kOffLane;
-    const uint32_t vx = forced ? 4u * (dxrow * N + c) : kOffLane;
     float u = 0.f;
     for (int t0 = 0; t0 < w.maxlen; t0 += TB) {
         const int tl = min(TB, w.maxlen - t0);
         if (w.onebuf && t0 + TB <= w.minlen) {
-            float zv[TB], xv[TB];
+            if (t0 > 0) {
 #pragma unroll
-            for (int tt = 0; tt < TB; ++tt) {
-                zv[tt] = bload(rz, vz, 4 * (t0 + tt) * M);
-                xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
+                for (int tt = 0; tt < TB; ++tt) {
+                    zv[tt] = bload(rz, vz, 4 * (t0 + tt) * M);
+                    xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
+                }
             }
-            // residual and masks of every step of the tile; r overwrites zv
+            // residual and masks of every step of the tile, two steps at a time; r overwrites zv
             uint32_t posb = 0u;
 #pragma unroll
-            for (int tt = 0; tt < TB; ++tt) {
+            for (int tt = 0; tt < TB; tt += 2) {
                 const int s = s0 + t0 + tt;
-                const float zt =
+                const float zt0 =
                     (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xv[tt]));
-                const bool pos = zt > 0.f;
-                posb |= (pos ? 1u : 0u) << tt;
-                const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
-                zprev = zv[tt];
-                zv[tt] = zv[tt] - F;
+                const float zt1 = !forced ? zv[tt] : __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt + 1]));
+                const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
+                posb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
+                float d0, d1;
+                row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
+                const float F0 = fmaf(Ai, zt0, d0) + hi, F1 = fmaf(Ai, zt1, d1) + hi;
+                zprev = zv[tt + 1];
+                zv[tt] = zv[tt] - F0;
+                zv[tt + 1] = zv[tt + 1] - F1;
             }
             // serial part: chunk products and chunk-local solutions
 #pragma unroll
@@ -1008,7 +1101,8 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
     if (w.maxlen == 0) return;
     const int id = chain0 + g;
     const bool okc = id < nchains;
-    const int b = okc ? id / ncs : 0, s0 = okc ? (id % ncs) * C : 0;
+    int b, s0;
+    chain_pos(chain0, g, nchains, ncs, C, b, s0);
     int len = 0;
     float gm = 1.f;
 #pragma unroll
@@ -1687,7 +1781,8 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
         for (int r = 0; r < 4; ++r) acc[n][r] = (4 * g + r == c) ? 1.f : 0.f;
     const int id = chain0 + g;
     const bool okc = id < nchains;
-    const int b = okc ? id / ncs : 0, s0 = okc ? (id % ncs) * C : 0;
+    int b, s0;
+    chain_pos(chain0, g, nchains, ncs, C, b, s0);
     int len = 0;
 #pragma unroll
     for (int n = 0; n < 4; ++n)
@@ -1900,7 +1995,8 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn16(const float *__restric
     const Chains16 w = chains16(chain0, nchains, ncs, C, T, nullptr, nullptr, nullptr);
     const int id = chain0 + g;
     const bool okc = id < nchains;
-    const int b = okc ? id / ncs : 0, s0 = okc ? (id % ncs) * C : 0;
+    int b, s0;
+    chain_pos(chain0, g, nchains, ncs, C, b, s0);
     int len = 0;
 #pragma unroll
     for (int n = 0; n < 4; ++n)

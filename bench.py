@@ -80,6 +80,9 @@ def kernel_work(c, steps, updates):
         # forward Newton updates run the fused kernel (residual + masks + product); the
         # adjoint runs the shifted product and a mask pass
         out["k_newton_product_plrnn"] = ("mfma", fwd * 2.0 * M ** 3)
+        # M <= 16 with whole blocks of chunks: one kernel per pass (the fix-up of an update and
+        # the forward pass of the next); its matrix-core work is the forward pass's
+        out["k_newton_pass16"] = ("mfma", fwd * 2.0 * M ** 3)
         out["k_chunk_product_plrnn"] = ("mfma", steps * B * (T - 1) * 2.0 * M ** 3)
         out["k_resjac_plrnn"] = ("hbm", adj * (4 * M + 4 * N + 4 * W))
         if M <= 16:
@@ -106,7 +109,7 @@ def kernel_work(c, steps, updates):
 # scaled by the reading of a plain copy of known size in the same run; kept in
 # profiles/traffic_<workload>.txt together with the hash of the kernel's source file, and
 # reported only while that source is unchanged.
-KERNEL_SOURCE = {"k_newton_product_plrnn": "k_plrnn.hip", "k_chunk_product_plrnn": "k_plrnn.hip",
+KERNEL_SOURCE = {"k_newton_product_plrnn": "k_plrnn.hip", "k_newton_pass16": "k_plrnn.hip", "k_chunk_product_plrnn": "k_plrnn.hip",
                  "k_fixup_fwd_plrnn": "k_plrnn.hip", "k_jacform_shplrnn": "k_shallow.hip",
                  "k_chunk_product_dense": "k_dense.hip", "k_readout": "k_readout.hip",
                  "k_diag_scan_lb_grads": "k_diag.hip", "k_diag_seg_write": "k_diag.hip"}

@@ -187,6 +187,13 @@ static int group_maps_override() {
     return e ? atoi(e) : -1;
 }
 
+// DEER_PASS_FUSION=0 keeps the M <= 16 fix-up and forward pass in separate kernels where the
+// fused pass kernel would apply (a test override)
+static bool pass_fusion_allowed() {
+    const char *e = getenv("DEER_PASS_FUSION");
+    return !e || atoi(e) != 0;
+}
+
 // Chunk length of the dense scans: enough chains to fill the machine (about 2048 waves),
 // and a bounded number of chunks per sequence so that the two-level carry pass stays short
 // (1024 for MP <= 32, 512 for MP = 64, whose group pass composes 64 x 64 maps).
@@ -208,25 +215,28 @@ static int choose_chunk(int B, int T, int MP) {
     return (int)C;
 }
 
-// Per-sequence control block of the Newton loop (device, 7B words, one device-to-host copy
-// reads all of it): act | gamma | sel | om | it | norm | status (see NewtonDev), then 2B
-// words of max bits for the fixed-iteration mode, the per-chain maxima of a pass, and the
-// second iterate buffer.
+// Per-sequence control block of the Newton loop (device, 8B words; one device-to-host copy of
+// the first 7B reads the results): act | gamma | sel | om | it | norm | status | pv (see
+// NewtonDev), then 2B words of max bits for the fixed-iteration mode, the per-chain maxima of
+// a pass, and the second iterate buffer.
 struct NewtonCtl {
     NewtonDev nd;
-    uint32_t *blk;          // start of the 7B-word block
+    uint32_t *blk;          // start of the 8B-word block
+    uint32_t *pv;           // its last B words (NewtonDev::pv of the fused passes)
     uint32_t *norm_bits;
     uint32_t *chain_bits;   // per-chain maxima [2][B * ncs] before the per-sequence reduction
     float *zalt;            // second iterate buffer [B,T,M]
     uint32_t *seq;          // kSeqWords per sequence: the fix-up's fused pass-end control
     bool fused;             // the update takes the pass-end control itself (no k_seq_ctl)
+    int lead;               // kernels queued before the first update completes (fused passes: 1)
 };
 
 static NewtonCtl carve_ctl(Carver &c, int B, size_t seq_elems, size_t nchains) {
     NewtonCtl n{};
-    uint32_t *blk = c.take<uint32_t>(7 * (size_t)B);
+    uint32_t *blk = c.take<uint32_t>(8 * (size_t)B);
     n.blk = blk;
     if (blk) {
+        n.pv = blk + 7 * (size_t)B;
         n.nd.act = (int *)blk;
         n.nd.gamma = (float *)(blk + B);
         n.nd.sel = (int *)(blk + 2 * B);
@@ -247,6 +257,7 @@ struct PlrnnWs {
     uint32_t *masks;
     float *P, *v, *carry, *gws;
     float *gmap;   // M <= 16, 32 | chunks: group maps [B][chunks / 32][16 x 16 + 16]
+    float *P2, *v2, *gmap2;   // the second set of aggregates of the fused passes (else null)
     NewtonCtl ctl;
     float *gpart;
     double *gpart2;
@@ -271,6 +282,12 @@ static PlrnnWs carve_plrnn(void *ws, int B, int T, int M, int op, size_t *bytes)
     const int gov = group_maps_override();
     const bool gm = w.MP == 16 && w.ncs % 32 == 0 && (gov < 0 ? nch >= 2048 : gov > 0);
     w.gmap = gm ? c.take<float>((size_t)B * (w.ncs / 32) * 272) : nullptr;
+    // fused passes: group maps, whole chunks of whole tiles
+    if (op == DEER_OP_SOLVE && gm && (long)w.C * w.ncs == T && w.C % 16 == 0 && pass_fusion_allowed()) {
+        w.P2 = c.take<float>(nch * 256);
+        w.v2 = c.take<float>(nch * 16);
+        w.gmap2 = c.take<float>((size_t)B * (w.ncs / 32) * 272);
+    }
     if (op == DEER_OP_SOLVE) {
         w.ctl = carve_ctl(c, B, (size_t)T * M, nch);
         w.r = c.take<float>((size_t)B * T * M);
@@ -492,16 +509,18 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
         int passes = 0;
         auto queue = [&]() {
             const int r = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt, mark, t_host.next_pass);
-            ++t_host.next_pass;
+            if (++t_host.next_pass == 0u) t_host.next_pass = 1u;   // 0 marks "no aggregates"
+
             ++passes;
             return r;
         };
+        const int cap = max_iter + ctl.lead;
         rc = queue();
-        if (!rc && passes < max_iter) rc = queue();
+        if (!rc && passes < cap) rc = queue();
         while (!rc) {
             if ((rc = wait_mark(mark, t_host.next_pass - 1, st))) break;
             if ((stopped = all_stopped())) break;
-            if (passes >= max_iter) break;
+            if (passes >= cap) break;
             rc = queue();
         }
         if (rc) return rc;
@@ -605,12 +624,24 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     // M <= 16: the fix-up also takes the pass-end control of the adaptive loop
     NewtonCtl ctl = w.ctl;
     ctl.fused = w.MP == 16 && o->fixed_iters <= 0;
+    // one kernel per pass: the fix-up of the previous update and the forward pass of the next
+    const bool pass16 = ctl.fused && w.P2;
+    if (pass16) {
+        ctl.nd.pv = ctl.pv;
+        ctl.lead = 1;
+    }
     uint32_t *mark_unused = nullptr;
     if (ctl.fused && (rc = host_block(B, ctl.nd, &mark_unused))) return rc;
     const FusedCtl fc{ctl.nd, ctl.seq, o->tol, o->step_bound == 0.f ? kDefaultStepBound : o->step_bound, kDamp};
     auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *mark,
                       uint32_t pass_no) -> int {
         int r;
+        if (pass16) {   // aggregates alternate between the two sets
+            const bool odd = pass_no & 1u;
+            return launch_newton_pass16(a, zb, za, odd ? w.P2 : w.P, odd ? w.v2 : w.v, odd ? w.gmap2 : w.gmap,
+                                        odd ? w.P : w.P2, odd ? w.v : w.v2, odd ? w.gmap : w.gmap2, w.C, w.ncs, fc,
+                                        mark, pass_no, st);
+        }
         // M <= 16: each wave's four chunks are composed in the forward pass, one kernel walks
         // the composed maps, and the fix-up applies the per-chunk prefix maps
         // 32 | chunks: the forward pass also composes each block's eight wave maps into a

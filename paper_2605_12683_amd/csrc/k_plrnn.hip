@@ -1023,8 +1023,10 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
 // freeze the sequence once max|Delta| < tol), or reject it (keep sel, raise the damping:
 // 1 - gamma = first, then x grow up to 1 = the fixed-point step); a non-finite fixed-point step
 // ends the sequence.
+// tag: with nd.pv, the number of the pass that may use the aggregates the caller's kernel
+// formed for the accepted iterate (it is stored when the update is kept and the sequence goes on)
 __device__ __forceinline__ void seq_decide(int b, uint32_t e, uint32_t zm, const NewtonDev &nd, float tol, float bound,
-                                           const NewtonDamp &dp) {
+                                           const NewtonDamp &dp, uint32_t tag = 0u) {
     const float ef = __uint_as_float(e), zf = __uint_as_float(zm);
     const bool fin = e < 0x7f800000u;
     float om = nd.om[b];
@@ -1047,6 +1049,7 @@ __device__ __forceinline__ void seq_decide(int b, uint32_t e, uint32_t zm, const
         nd.norm[b] = ef;
         if (om > 0.f) om = om / dp.shrink < dp.floor ? 0.f : om / dp.shrink;
         if (ef < tol) stop(it, 1);
+        else if (nd.pv) nd.pv[b] = tag;
     } else if (om >= 1.f) {
         nd.norm[b] = ef;
         stop(nd.it[b], 2);
@@ -1060,7 +1063,8 @@ __device__ __forceinline__ void seq_decide(int b, uint32_t e, uint32_t zm, const
 // Arrival of `cnt` chains of sequence b with maxima e, zm (see FusedCtl).  Device-scope atomics
 // meet at one coherence point across the XCDs; each maximum is returned (so performed) before
 // the count is raised, so the chain that completes the count reads the final maxima.
-__device__ __forceinline__ void seq_arrive(const FusedCtl &fc, int b, int cnt, int ncs, uint32_t e, uint32_t zm) {
+__device__ __forceinline__ void seq_arrive(const FusedCtl &fc, int b, int cnt, int ncs, uint32_t e, uint32_t zm,
+                                           uint32_t tag = 0u) {
     uint32_t *blk = fc.seq + (size_t)b * kSeqWords;   // count | max |Delta| | max |z|, 128 bytes apart
     const uint32_t r1 = __hip_atomic_fetch_max(blk + 32, e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t r2 = __hip_atomic_fetch_max(blk + 64, zm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1071,7 +1075,7 @@ __device__ __forceinline__ void seq_arrive(const FusedCtl &fc, int b, int cnt, i
     if (old + (uint32_t)cnt != (uint32_t)ncs) return;
     const uint32_t ef = __hip_atomic_load(blk + 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t zf = __hip_atomic_load(blk + 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    seq_decide(b, ef, zf, fc.nd, fc.tol, fc.bound, fc.dp);
+    seq_decide(b, ef, zf, fc.nd, fc.tol, fc.bound, fc.dp, tag);
     __hip_atomic_store(blk + 32, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(blk + 64, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(blk, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1307,6 +1311,411 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
             seq_arrive(fc, bn, cnt, ncs, E, Z);
         }
     }
+}
+
+// ---------------------------------------------------------------------------------------
+// One kernel per Newton pass (M <= 16).  Where every sequence is a whole number of blocks of 32
+// chunks of whole tiles, the fix-up of pass p and the forward pass of update p + 1 run in one
+// kernel: a wave walks the group maps to its carry, takes its four chunks through pass p's
+// update (z + Delta written out and kept in registers), and then forms the chunk products and
+// chunk-local solutions of the next update on the new iterate, so the tile is loaded once and
+// the start-up of the second kernel (control words, weights, tile loads) disappears.
+// The next update is formed before the sequence's decision on pass p is known, with the
+// damping an accepted update leads to; the decision stores in nd.pv that the aggregates belong
+// to the new iterate only when the update is kept and the sequence goes on.  A sequence
+// without valid aggregates (the first kernel, or after a rejected update) runs only the
+// forward pass on its current iterate in the next kernel.  Aggregates alternate between two
+// buffers (the kernel reads one and writes the other).
+// The forward pass of a chunk needs the new iterate at the step before it.  Inside a wave it
+// comes from the row before; for a wave's first chunk it is z + Delta with Delta the chunk's
+// carry, and the previous wave puts exactly that value at its last step (it forms the next
+// wave's carry with the same operations on the same operands instead of taking the end of its
+// own recurrence, the same Delta to rounding), so no wave waits for another.
+// ---------------------------------------------------------------------------------------
+template <int TB>
+__global__ __launch_bounds__(512) void k_newton_pass16(
+    const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
+    const float *__restrict__ x, const float *__restrict__ z0, float *zbuf, float *zalt, int T, int M, int C, int ncs,
+    const float *__restrict__ Pin, const float *__restrict__ vin, const float *__restrict__ gin,
+    float *__restrict__ Pout, float *__restrict__ vout, float *__restrict__ gout, FusedCtl fc, uint32_t *mark,
+    uint32_t pass_no) {
+    constexpr int WPB = 8;
+    const int lane = threadIdx.x & 63, wvb = rfl_i((int)(threadIdx.x >> 6)), g = lane >> 4, c = lane & 15;
+    if (mark && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(mark, pass_no, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    const NewtonDev &nd = fc.nd;
+    // a block's 32 chunks belong to one sequence b
+    const int chain0 = (blockIdx.x * WPB + wvb) * 4;
+    const int b = chain0 / ncs, cc0 = chain0 - b * ncs;
+    if (nd.act[b] == 0) return;   // the whole block
+    const bool have = nd.pv[b] == pass_no;
+    const int sel = nd.sel[b];
+    const float gam = nd.gamma[b];
+    float omn = nd.om[b];   // the damping of the next update if this one is kept
+    if (omn > 0.f) omn = omn / fc.dp.shrink < fc.dp.floor ? 0.f : omn / fc.dp.shrink;
+    const float gnext = have ? 1.f - omn : gam;
+    float *const zc = sel ? zalt : zbuf;   // current iterate
+    float *const zn = sel ? zbuf : zalt;   // the update's output
+    const int s0 = (cc0 + g) * C;          // first step of this lane's chunk
+    const bool lat = c < M, forced = c < N;
+    const size_t row0 = (size_t)b * T + (size_t)cc0 * C, xrow0 = (size_t)b * (T + 1) + (size_t)cc0 * C;
+    const auto rzc = wave_rsrc(zc + row0 * M), rzn = wave_rsrc(zn + row0 * M);
+    const auto rx = wave_rsrc(N > 0 ? x + xrow0 * N : zc);
+    const uint32_t vz = lat ? 4u * ((uint32_t)(g * C) * M + c) : kOffLane;
+    const uint32_t vx = forced ? 4u * ((uint32_t)(g * C) * N + c) : kOffLane;
+    // the first tile's loads go out first; the weights come through LDS (one load per element
+    // for the block instead of gathers by every wave)
+    float zv[TB], xv[TB];
+#pragma unroll
+    for (int tt = 0; tt < TB; ++tt) {
+        zv[tt] = bload(rzc, vz, 4 * tt * M);
+        xv[tt] = bload(rx, vx, 4 * tt * N);
+    }
+    float zprev = 0.f;   // z_{s0-1} of the current iterate (the initial state at s0 = 0)
+    if (lat) {
+        if (s0 == 0) zprev = z0 ? z0[(size_t)b * M + c] : (forced ? x[(size_t)b * (T + 1) * N + c] : 0.f);
+        else zprev = zc[((size_t)b * T + s0 - 1) * M + c];
+    }
+    __shared__ float sW[256], sA[16], sH[16];
+    {
+        const int t = threadIdx.x;
+        if (t < M * M) sW[t] = W[t];
+        if (t < M) {
+            sA[t] = A[t];
+            sH[t] = h ? h[t] : 0.f;
+        }
+    }
+    lds_barrier();
+    int src[16];
+    row_sources(c, src);
+    float wr[16], wp[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        wr[k] = (lat && src[k] < M) ? sW[c * M + src[k]] : 0.f;
+        wp[k] = wr[k] * p_of(src[k], N, alpha);
+    }
+    const float Ai = lat ? sA[c] : 0.f, hi = lat ? sH[c] : 0.f;
+    const float pi = p_of(c, N, alpha), di = Ai * pi;
+    float WpD[4], Dq[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int col = 4 * g + q;
+        const float wpq = (c < M && col < M) ? sW[c * M + col] * p_of(col, N, alpha) : 0.f;
+        Dq[q] = (col == c && col < M) ? sA[col] * p_of(col, N, alpha) : 0.f;
+        WpD[q] = wpq + Dq[q];
+    }
+    // ---- fix-up of the current update: the carry of this lane's chunk ----
+    float D = 0.f, Dnext = 0.f;
+    bool nextc = false;   // this lane's chunk ends where the next wave's starts
+    if (have) {
+        const int ngm = ncs / 32, grp = cc0 / 32;
+        const float *Gb = gin + (size_t)b * ngm * 272;
+        v4f cur = {0.f, 0.f, 0.f, 0.f};
+        constexpr int PF = 4;
+        float ga[PF][4], gv[PF][4];
+        if (grp > 0) {
+#pragma unroll
+            for (int d2 = 0; d2 < PF; ++d2) {
+                const float *Gk = Gb + (size_t)min(d2, grp - 1) * 272;
+                carry16_fetch<false>(Gk, Gk + 256, g, c, ga[d2], gv[d2]);
+            }
+        }
+        for (int k0 = 0; k0 < grp; k0 += PF) {
+#pragma unroll
+            for (int d2 = 0; d2 < PF; ++d2) {
+                if (k0 + d2 >= grp) break;
+                v4f nx = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) nx = mfma16x16x4(ga[d2][q], cur[q], nx);
+                if (c == 0) {
+#pragma unroll
+                    for (int r2 = 0; r2 < 4; ++r2) nx[r2] += gv[d2][r2];
+                }
+                cur = nx;
+                const float *Gk = Gb + (size_t)min(k0 + d2 + PF, grp - 1) * 272;
+                carry16_fetch<false>(Gk, Gk + 256, g, c, ga[d2], gv[d2]);
+            }
+        }
+        // the wave's carry: its prefix within the group (slot chain0) applied to the group's
+        // carry; element k sits in lane 16 (k / 4), register k % 4, and is read as a scalar
+        float wa[4], wvv[4];
+        carry16_fetch<false>(Pin + (size_t)chain0 * 256, vin + (size_t)chain0 * 16, g, c, wa, wvv);
+        v4f wc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) wc = mfma16x16x4(wa[q], cur[q], wc);
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) wc[r2] += wvv[r2];
+        float wk[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            wk[k] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wc[k & 3]), 16 * (k >> 2)));
+        if (g == 0) {
+            float dv = wk[0];
+#pragma unroll
+            for (int k = 1; k < 16; ++k) dv = c == k ? wk[k] : dv;
+            D = dv;
+        } else {   // chunk g of the wave: R_g carry(wave) + s_g
+            const float4 *R4 = reinterpret_cast<const float4 *>(Pin + (size_t)(chain0 + g) * 256 + c * 16);
+            float a0 = vin[(size_t)(chain0 + g) * 16 + c], a1 = 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 rr4 = R4[q];
+                a0 = fmaf(rr4.x, wk[4 * q], a0);
+                a1 = fmaf(rr4.y, wk[4 * q + 1], a1);
+                a0 = fmaf(rr4.z, wk[4 * q + 2], a0);
+                a1 = fmaf(rr4.w, wk[4 * q + 3], a1);
+            }
+            D = a0 + a1;
+        }
+        if (!lat) D = 0.f;
+        // The carry of the next wave's first chunk, formed with the same operations on the same
+        // operands as that wave forms it (one more group step when it starts the next group),
+        // so both waves put the same z + Delta at the step between them.
+        if (cc0 + 4 < ncs) {
+            v4f curn = cur;
+            if ((cc0 + 4) / 32 != grp) {
+                float ga1[4], gv1[4];
+                carry16_fetch<false>(Gb + (size_t)grp * 272, Gb + (size_t)grp * 272 + 256, g, c, ga1, gv1);
+                v4f nx = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) nx = mfma16x16x4(ga1[q], curn[q], nx);
+                if (c == 0) {
+#pragma unroll
+                    for (int r2 = 0; r2 < 4; ++r2) nx[r2] += gv1[r2];
+                }
+                curn = nx;
+            }
+            float wa2[4], wv2[4];
+            carry16_fetch<false>(Pin + (size_t)(chain0 + 4) * 256, vin + (size_t)(chain0 + 4) * 16, g, c, wa2, wv2);
+            v4f wcn = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) wcn = mfma16x16x4(wa2[q], curn[q], wcn);
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) wcn[r2] += wv2[r2];
+            float dn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wcn[0]), 0));
+#pragma unroll
+            for (int kk = 1; kk < 16; ++kk) {
+                const float e = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wcn[kk & 3]), 16 * (kk >> 2)));
+                dn = c == kk ? e : dn;
+            }
+            if (g == 3 && lat) Dnext = dn;
+            nextc = g == 3;
+        }
+    }
+    // z_{s0-1} of the iterate the next update is formed at
+    float zpn = have ? zprev + D : zprev;
+    uint32_t emax = 0u, zmax = 0u;
+    if (have) {
+        // residual and masks at the current iterate, then Delta_t = gamma J~_t Delta_{t-1} - r_t;
+        // the new iterate is written out and, in the last tile, kept in zv
+        for (int t0 = 0; t0 < C; t0 += TB) {
+            if (t0 > 0) {
+#pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    zv[tt] = bload(rzc, vz, 4 * (t0 + tt) * M);
+                    xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
+                }
+            }
+            float rv[TB];
+            uint32_t mb = 0u;
+#pragma unroll
+            for (int tt = 0; tt < TB; tt += 2) {
+                const int s = s0 + t0 + tt;
+                const float zt0 =
+                    (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xv[tt]));
+                const float zt1 = !forced ? zv[tt] : __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt + 1]));
+                const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
+                mb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
+                float d0, d1;
+                row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
+                rv[tt] = zv[tt] - (fmaf(Ai, zt0, d0) + hi);
+                rv[tt + 1] = zv[tt + 1] - (fmaf(Ai, zt1, d1) + hi);
+                zprev = zv[tt + 1];
+            }
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                const bool m = (mb >> tt) & 1u;
+                const float y = fmaf(di, D, row16_dot(wp, m ? D : 0.f));
+                D = fmaf(gam, y, -rv[tt]);
+                const float zcur = zv[tt];
+                // the last step before the next wave: its Delta as that wave's carry
+                const float dap = (tt == TB - 1 && t0 + TB == C && nextc) ? Dnext : D;
+                const float znew = zcur + dap;
+                if (t0 + TB < C) bstore_u(rzn, __float_as_uint(znew), vz, 4 * (t0 + tt) * M);
+                const uint32_t ab = lat ? abs_bits(dap) : 0u, zb = abs_bits(zcur);
+                emax = emax > ab ? emax : ab;
+                zmax = zmax > zb ? zmax : zb;
+                zv[tt] = znew;
+            }
+        }
+        // z_{s0-1} of the new iterate exactly as stored: chunks 1..3 of the wave take it from the
+        // row before; the first chunk's own carry equals the previous wave's (see above)
+        const float zlast = __shfl(zv[TB - 1], (lane - 16) & 63, 64);
+        if (g > 0) zpn = zlast;
+        // the last tile of the new iterate; chunks of several tiles read it back
+#pragma unroll
+        for (int tt = 0; tt < TB; ++tt) bstore_u(rzn, __float_as_uint(zv[tt]), vz, 4 * (C - TB + tt) * M);
+        if (C > TB) __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
+    }
+    // ---- the next update's forward pass ----
+    const auto rzp = have ? rzn : rzc;   // the iterate it is formed at
+    v4f acc[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[n][r] = (4 * g + r == c) ? 1.f : 0.f;
+    float u = 0.f;
+    float gp = 1.f;   // gnext^TB: the damping of a tile's chunk product
+#pragma unroll
+    for (int k = 0; k < TB; ++k) gp *= gnext;
+    for (int t0 = 0; t0 < C; t0 += TB) {
+        if (C > TB && (have || t0 > 0)) {
+#pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                zv[tt] = bload(rzp, vz, 4 * (t0 + tt) * M);
+                xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
+            }
+        }
+        // residual and masks; r overwrites zv
+        uint32_t posb = 0u;
+#pragma unroll
+        for (int tt = 0; tt < TB; tt += 2) {
+            const int s = s0 + t0 + tt;
+            const float zt0 = (s == 0 || !forced) ? zpn : __fadd_rn(__fmul_rn(pi, zpn), __fmul_rn(alpha, xv[tt]));
+            const float zt1 = !forced ? zv[tt] : __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt + 1]));
+            const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
+            posb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
+            float d0, d1;
+            row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
+            const float F0 = fmaf(Ai, zt0, d0) + hi, F1 = fmaf(Ai, zt1, d1) + hi;
+            zpn = zv[tt + 1];
+            zv[tt] = zv[tt] - F0;
+            zv[tt + 1] = zv[tt + 1] - F1;
+        }
+#pragma unroll
+        for (int tt = 0; tt < TB; ++tt) {
+            const bool pos = (posb >> tt) & 1u;
+            const uint64_t bal = __ballot(pos);
+            float Am[4][4];
+#pragma unroll
+            for (int n = 0; n < 4; ++n)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
+                    Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+                }
+            v4f nx[4];
+#pragma unroll
+            for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int n = 0; n < 4; ++n) nx[n] = mfma16x16x4(Am[n][q], acc[n][q], nx[n]);
+#pragma unroll
+            for (int n = 0; n < 4; ++n) acc[n] = nx[n];
+            const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
+            u = fmaf(gnext, y, -zv[tt]);
+        }
+        if (gnext != 1.f) {
+#pragma unroll
+            for (int n = 0; n < 4; ++n)
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2) acc[n][r2] *= gp;
+        }
+    }
+    if (!lat) u = 0.f;
+    // ---- pass-end control of the current update (once per wave: its chunks share b) ----
+    if (have) {
+        emax = wave_max_u32(emax);
+        zmax = wave_max_u32(zmax);
+        if (lane == 0) seq_arrive(fc, b, 4, ncs, emax, zmax, pass_no + 1u);
+    } else if (lane == 0) {
+        // aggregates of the current iterate (nothing else of this sequence runs in this kernel)
+        nd.pv[b] = pass_no + 1u;
+    }
+    // ---- wave maps and group maps of the next update (as in k_newton_product_plrnn16) ----
+    __shared__ float lt[WPB][3][16][17];
+    __shared__ float lv[WPB][4][16];
+#pragma unroll
+    for (int n = 1; n < 4; ++n)
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) lt[wvb][n - 1][4 * g + r2][c] = acc[n][r2];
+    lv[wvb][g][c] = u;
+    lds_barrier();
+    float Am[3][4];
+    v4f bv[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int n = 1; n < 4; ++n) Am[n - 1][q] = lt[wvb][n - 1][c][4 * g + q];
+#pragma unroll
+        for (int n = 0; n < 4; ++n) bv[n][q] = c == 0 ? lv[wvb][n][4 * g + q] : 0.f;
+    }
+    v4f R2 = {0.f, 0.f, 0.f, 0.f}, R3 = {0.f, 0.f, 0.f, 0.f}, Qw = {0.f, 0.f, 0.f, 0.f};
+    v4f s2 = bv[1], s3 = bv[2], uw = bv[3];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        R2 = mfma16x16x4(Am[0][q], acc[0][q], R2);
+        s2 = mfma16x16x4(Am[0][q], bv[0][q], s2);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        R3 = mfma16x16x4(Am[1][q], R2[q], R3);
+        s3 = mfma16x16x4(Am[1][q], s2[q], s3);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        Qw = mfma16x16x4(Am[2][q], R3[q], Qw);
+        uw = mfma16x16x4(Am[2][q], s3[q], uw);
+    }
+    const v4f outm[3] = {acc[0], R2, R3}, outv[3] = {bv[0], s2, s3};
+#pragma unroll
+    for (int n = 1; n < 4; ++n) {
+        float *P = Pout + (size_t)(chain0 + n) * 256;
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) P[(4 * g + r2) * 16 + c] = outm[n - 1][r2];
+        if (c == 0)
+            *reinterpret_cast<float4 *>(vout + (size_t)(chain0 + n) * 16 + 4 * g) =
+                make_float4(outv[n - 1][0], outv[n - 1][1], outv[n - 1][2], outv[n - 1][3]);
+    }
+    __shared__ float lq[WPB][16][17];
+    __shared__ float lu[WPB][16];
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2) lq[wvb][4 * g + r2][c] = Qw[r2];
+    if (c == 0) {
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) lu[wvb][4 * g + r2] = uw[r2];
+    }
+    __syncthreads();
+    if (wvb != 0) return;
+    const int bc0 = blockIdx.x * WPB * 4;   // the block's first chain
+    v4f Gm, gu = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2) Gm[r2] = (4 * g + r2 == c) ? 1.f : 0.f;
+    for (int k = 0; k < WPB; ++k) {
+        float *P = Pout + (size_t)(bc0 + 4 * k) * 256;
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) P[(4 * g + r2) * 16 + c] = Gm[r2];
+        if (c == 0)
+            *reinterpret_cast<float4 *>(vout + (size_t)(bc0 + 4 * k) * 16 + 4 * g) =
+                make_float4(gu[0], gu[1], gu[2], gu[3]);
+        v4f ng = {0.f, 0.f, 0.f, 0.f}, nu;
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) nu[r2] = c == 0 ? lu[k][4 * g + r2] : 0.f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float aq = lq[k][c][4 * g + q];
+            ng = mfma16x16x4(aq, Gm[q], ng);
+            nu = mfma16x16x4(aq, gu[q], nu);
+        }
+        Gm = ng;
+        gu = nu;
+    }
+    const int ngm = ncs / (4 * WPB);
+    float *Gp = gout + ((size_t)b * ngm + cc0 / (4 * WPB)) * 272;
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2) Gp[(4 * g + r2) * 16 + c] = Gm[r2];
+    if (c == 0) *reinterpret_cast<float4 *>(Gp + 256 + 4 * g) = make_float4(gu[0], gu[1], gu[2], gu[3]);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -2399,6 +2808,7 @@ __global__ void k_ctl_init(NewtonDev nd, uint32_t *seq, int B) {
     nd.it[b] = 0;
     nd.norm[b] = __uint_as_float(0x7fc00000u);
     nd.status[b] = 0;
+    if (nd.pv) nd.pv[b] = 0u;   // no aggregates yet (pass numbers start at 1)
 }
 
 int launch_ctl_init(const NewtonDev &nd, uint32_t *seq, int B, hipStream_t st) {
@@ -2630,6 +3040,24 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
     } else if (MP == 32) NP(32); else NP(64);
 #undef NP
     DEER_LAUNCH_CHECK("k_newton_product_plrnn");
+    return DEER_OK;
+}
+
+int launch_newton_pass16(const PlrnnArgs &a, float *z, float *zalt, const float *Pin, const float *vin,
+                         const float *gin, float *Pout, float *vout, float *gout, int C, int ncs, const FusedCtl &fc,
+                         uint32_t *mark, uint32_t pass_no, hipStream_t st) {
+    if (a.M > 16 || ncs % 32 || C % 16 || (long)C * ncs != a.T || !fc.seq || !fc.nd.pv || !Pin || !vin || !gin ||
+        !Pout || !vout || !gout)
+        return invalid_arg("fused Newton passes need M <= 16, 32 | chunks, 16 | C, T = C chunks, the control and "
+                           "two aggregate buffers");
+    KTimer kt("k_newton_pass16", st);
+    const int grid = a.B * ncs / 32;
+#define NPS(TBV)                                                                                                  \
+    hipLaunchKernelGGL(k_newton_pass16<TBV>, dim3(grid), dim3(512), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, \
+                       z, zalt, a.T, a.M, C, ncs, Pin, vin, gin, Pout, vout, gout, fc, mark, pass_no)
+    if (C % 32) NPS(16); else NPS(32);
+#undef NPS
+    DEER_LAUNCH_CHECK("k_newton_pass16");
     return DEER_OK;
 }
 

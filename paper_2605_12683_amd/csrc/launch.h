@@ -66,6 +66,9 @@ struct NewtonDev {
     int *hit;
     float *hnorm;
     int *hstat;
+    // fused passes only (else null): number of the pass whose kernel may use the chunk
+    // aggregates stored for the sequence's current iterate (see launch_newton_pass16)
+    uint32_t *pv;
 };
 struct NewtonDamp {
     float first, grow, shrink, floor;
@@ -82,6 +85,14 @@ struct FusedCtl {
     NewtonDamp dp;
 };
 constexpr int kSeqWords = 96;
+// One kernel per Newton pass (M <= 16, adaptive loop, every sequence a whole number of blocks of
+// 32 chunks of C steps, C a multiple of 16): the fix-up of the previous pass from the aggregates
+// in (Pin, vin, gin), where fc.nd.pv says they belong to the current iterate, then the forward
+// pass of the next update on the new iterate, its aggregates written to (Pout, vout, gout).
+// Block 0 writes pass_no to *mark as it starts.
+int launch_newton_pass16(const PlrnnArgs &a, float *z, float *zalt, const float *Pin, const float *vin,
+                         const float *gin, float *Pout, float *vout, float *gout, int C, int ncs, const FusedCtl &fc,
+                         uint32_t *mark, uint32_t pass_no, hipStream_t st);
 int launch_ctl_init(const NewtonDev &nd, uint32_t *seq, int B, hipStream_t st);
 int launch_seq_max(const uint32_t *chain_bits, const int *active, uint32_t *norm_bits, int B, int ncs,
                    hipStream_t st);

@@ -25,10 +25,10 @@ TOL = 1e-4
 
 @pytest.fixture(autouse=True)
 def _no_chunk_override():
-    for k in ("DEER_CHUNK", "DEER_GROUP_MAPS"):
+    for k in ("DEER_CHUNK", "DEER_GROUP_MAPS", "DEER_PASS_FUSION"):
         os.environ.pop(k, None)
     yield
-    for k in ("DEER_CHUNK", "DEER_GROUP_MAPS"):
+    for k in ("DEER_CHUNK", "DEER_GROUP_MAPS", "DEER_PASS_FUSION"):
         os.environ.pop(k, None)
 
 
@@ -98,6 +98,29 @@ def test_solve_reaches_rollout(M, N, B, T, alpha, chunk):
     got = masks_to_bool(res["masks"].cpu().numpy(), M)
     far = np.abs(zt) > 1e-4 * np.abs(zt).max()
     assert np.array_equal(got[far], (zt > 0)[far])
+
+
+@pytest.mark.parametrize("M,N,B,T,alpha,chunk,bound", [(16, 3, 2, 2048, 0.2, 16, 0.0), (12, 4, 2, 4096, 0.2, 32, 0.0),
+                                                       (16, 3, 3, 512, 0.2, 16, 0.3), (9, 9, 2, 2048, 0.15, 64, 0.0)])
+def test_fused_and_separate_pass_kernels_agree(M, N, B, T, alpha, chunk, bound):
+    """Where every sequence is whole blocks of 32 chunks of whole tiles, one kernel per pass
+    runs the fix-up of an update and the forward pass of the next; DEER_PASS_FUSION=0 keeps
+    them apart.  Both reach the rollout, with the same iteration counts up to one."""
+    os.environ["DEER_CHUNK"] = str(chunk)
+    os.environ["DEER_GROUP_MAPS"] = "1"
+    c = _case(M, N, B, T, alpha, 700 + M + T)
+    m = oracle_model(c)
+    ref = O.rollout(m, c.x, alpha, N)
+    out = {}
+    for fuse in ("1", "0"):
+        os.environ["DEER_PASS_FUSION"] = fuse
+        say("deer_solve fused" if fuse == "1" else "deer_solve separate", M, N, B, T, alpha, chunk, bound)
+        res = D.deer_solve(m, c.x, alpha, N, tol=1e-5, max_iter=5000, step_bound=bound)
+        assert res["status"] == 0, res
+        assert rel_inf(res["z"].cpu().numpy(), ref) < TOL
+        assert all(n < 1e-5 for n in res["norms"])
+        out[fuse] = res["iters"]
+    assert max(abs(a - b) for a, b in zip(out["1"], out["0"])) <= 1
 
 
 @pytest.mark.parametrize("M,N,B,T,alpha,chunk,bound", [(16, 3, 4, 300, 0.2, 0, 0.05), (16, 3, 3, 300, 0.2, 16, 0.3),

@@ -93,6 +93,14 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// The same for data exchanged through LDS between the lanes of one wave only: the LDS writes
+// complete before the reads after it, and no other wave is waited for.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ float forced_state(const float *__restrict__ x, const float *__restrict__ z0,
                                               const float *__restrict__ z, int b, int s, int i, int T, int M,
                                               int N, float alpha) {

@@ -924,7 +924,7 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
 #pragma unroll
             for (int r2 = 0; r2 < 4; ++r2) lt[wvb][n - 1][4 * g + r2][c] = acc[n][r2];
         lv[wvb][g][c] = u;
-        lds_barrier();
+        wave_lds_sync();   // each wave's own slots
         float Am[3][4];
         v4f bv[4];
 #pragma unroll
@@ -1641,7 +1641,7 @@ __global__ __launch_bounds__(512) void k_newton_pass16(
 #pragma unroll
         for (int r2 = 0; r2 < 4; ++r2) lt[wvb][n - 1][4 * g + r2][c] = acc[n][r2];
     lv[wvb][g][c] = u;
-    lds_barrier();
+    wave_lds_sync();   // each wave's own slots
     float Am[3][4];
     v4f bv[4];
 #pragma unroll

@@ -9,6 +9,7 @@
 #include <map>
 #include <mutex>
 #include <string>
+#include <chrono>
 #include <vector>
 
 #include "common.h"
@@ -446,13 +447,16 @@ static int host_block(int B, NewtonDev &nd, uint32_t **mark) {
     return DEER_OK;
 }
 
-// Waits until the pass mark has reached `want` (in wrapping order).  The stream is queried now
-// and then, so that a stream that ran dry without the mark is an error, not a hang.
+// Waits until the pass mark has reached `want` (in wrapping order).  The stream is queried only
+// after a long wait (a runtime call while the device works delays the following kernels), so
+// that a stream that ran dry without the mark is an error, not a hang.
 static int wait_mark(const uint32_t *mark, uint32_t want, hipStream_t st) {
     auto reached = [&]() { return (int32_t)(__atomic_load_n(mark, __ATOMIC_ACQUIRE) - want) >= 0; };
+    using clk = std::chrono::steady_clock;
+    const auto t0 = clk::now();
     for (unsigned spin = 1;; ++spin) {
         if (reached()) return DEER_OK;
-        if ((spin & 1023u) == 0u) {
+        if ((spin & 4095u) == 0u && clk::now() - t0 > std::chrono::milliseconds(200)) {
             const hipError_t e = hipStreamQuery(st);
             if (e == hipSuccess) {
                 if (reached()) return DEER_OK;
@@ -504,13 +508,15 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
         // when every earlier pass, and so the decisions of pass p - 1, is complete.  The host
         // keeps one pass queued ahead: once pass p has started it reads the flags as of pass
         // p - 1 and queues pass p + 1 (a whole pass of time to do so), so the device does not
-        // wait for the host and one pass runs past convergence (it skips every sequence).
-        // The loop ends only after the mark of the last queued pass, so no mark is pending.
+        // wait for the host and one pass runs past convergence (it skips every sequence).  The
+        // loop ends only after the mark of the last queued pass, so no mark is pending.
         int passes = 0;
+        uint32_t last = 0u;   // number of the last pass queued
         auto queue = [&]() {
-            const int r = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt, mark, t_host.next_pass);
+            const uint32_t no = t_host.next_pass;
+            const int r = update(nd.act, nd.gamma, nd.sel, z, ctl.zalt, mark, no);
             if (++t_host.next_pass == 0u) t_host.next_pass = 1u;   // 0 marks "no aggregates"
-
+            last = no;
             ++passes;
             return r;
         };
@@ -518,7 +524,7 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
         rc = queue();
         if (!rc && passes < cap) rc = queue();
         while (!rc) {
-            if ((rc = wait_mark(mark, t_host.next_pass - 1, st))) break;
+            if ((rc = wait_mark(mark, last, st))) break;
             if ((stopped = all_stopped())) break;
             if (passes >= cap) break;
             rc = queue();

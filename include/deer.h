@@ -164,6 +164,25 @@ int deer_adjoint(const deer_model *model, const deer_forcing *forcing, int B, in
                  const float *x, const float *z0, const float *z, const float *g,
                  float *lam, const deer_grads *grads, void *ws, size_t ws_bytes, void *stream);
 
+/* Sequential GTF baseline (the comparison of Fig. 1A): the forward rollout
+ *   z_s = F(z~_s), z~ the forced state of eq. GTF, step by step in time,
+ * and, when lam or grads is given, back-propagation through time, also step by step:
+ *   lam_{T-1} = g_{T-1},  lam_s = g_s + J~_{s+1}^T lam_{s+1},  dL/dtheta = sum lam_s^T dF/dtheta.
+ * The outputs are those of deer_solve at convergence and deer_adjoint at its z, computed in
+ * time order with the batch as the only parallel dimension (one workgroup per sequence):
+ * the training the parallel solver replaces.  PLRNN kinds only; M <= 256, L <= 256,
+ * M L <= 8192 (vanilla: M^2 <= 8192), and the weights must fit in 160 KiB of LDS.
+ *   x, z0        as in deer_solve;  z [B,T,M] out.
+ *   g            [B,T,M] or NULL (the MSE seed, as in deer_adjoint).
+ *   lam          [B,T,M] out or NULL;  grads as in deer_adjoint or NULL (then no backward pass
+ *                when lam is NULL too).
+ *   ws           deer_sequential_workspace_bytes(model, B, T) bytes.
+ * Fully asynchronous on `stream`. */
+int deer_sequential(const deer_model *model, const deer_forcing *forcing, int B, int T,
+                    const float *x, const float *z0, float *z, const float *g, float *lam,
+                    const deer_grads *grads, void *ws, size_t ws_bytes, void *stream);
+size_t deer_sequential_workspace_bytes(const deer_model *model, int B, int T);
+
 /* Layout of the cotangent g of deer_adjoint_ex. */
 enum { DEER_G_NATIVE = 0, DEER_G_REAL = 1 };
 

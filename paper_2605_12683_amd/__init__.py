@@ -20,7 +20,8 @@ from . import _binding as _b
 from ._binding import DeerError, load  # noqa: F401
 
 __all__ = ["deer_solve", "deer_adjoint", "deer_readout_loss", "plrnn_jacobian", "deer_scan", "deer_workspace_bytes",
-           "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_status_string", "DeerError", "load"]
+           "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_status_string", "DeerError", "load",
+           "deer_sequential", "deer_sequential_workspace_bytes"]
 
 _KINDS = {"plrnn": _b.DEER_PLRNN, "shplrnn": _b.DEER_SHPLRNN, "diag_ssm": _b.DEER_DIAG_SSM}
 _INITS = {"teacher": _b.DEER_INIT_TEACHER, "zero": _b.DEER_INIT_ZERO, "user": _b.DEER_INIT_USER}
@@ -222,6 +223,45 @@ def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, w
                              g_layout, _ptr(lam), ctypes.byref(gs), _ptr(ws), ws.numel(), _stream())
     _b._check(st, "deer_adjoint")
     return {"lam": lam, "grads": grads}
+
+
+def _plrnn_grads(m):
+    """Gradient outputs of a PLRNN-kind model and the C struct pointing at them."""
+    if m.kind == "plrnn":
+        grads = {"A": torch.empty(m.M, device="cuda"), "W": torch.empty(m.M, m.M, device="cuda"),
+                 "h": torch.empty(m.M, device="cuda")}
+        return grads, _b.deer_grads(_ptr(grads["A"]), _ptr(grads["W"]), None, _ptr(grads["h"]), None)
+    grads = {"A": torch.empty(m.M, device="cuda"), "W1": torch.empty(m.M, m.L, device="cuda"),
+             "W2": torch.empty(m.L, m.M, device="cuda"), "h1": torch.empty(m.M, device="cuda"),
+             "h2": torch.empty(m.L, device="cuda")}
+    return grads, _b.deer_grads(_ptr(grads["A"]), _ptr(grads["W1"]), _ptr(grads["W2"]), _ptr(grads["h1"]),
+                                _ptr(grads["h2"]))
+
+
+def deer_sequential(model, x, alpha: float, n_forced: int, *, z0=None, g=None, want_lam: bool = True,
+                    want_grads: bool = True, ws=None, z=None) -> dict:
+    """Sequential GTF baseline: the rollout z and, if asked, back-propagation through time (lam
+    and the parameter gradients), step by step in time.  Returns dict(z, lam, grads)."""
+    lib = load()
+    m = _model(model)
+    x = _dev(x)
+    B, T1, _ = x.shape
+    T = T1 - 1
+    out = torch.empty(B, T, m.M, device="cuda") if z is None else z
+    lam = torch.empty(B, T, m.M, device="cuda") if want_lam else None
+    grads, gs = _plrnn_grads(m) if want_grads else ({}, None)
+    if ws is None:
+        ws = _workspace(lib.deer_sequential_workspace_bytes(ctypes.byref(m.c), B, T))
+    f = _b.deer_forcing(float(alpha), int(n_forced))
+    z0d, gd = _dev(z0), _dev(g)
+    st = lib.deer_sequential(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(out), _ptr(gd),
+                             _ptr(lam), ctypes.byref(gs) if gs is not None else None, _ptr(ws), ws.numel(), _stream())
+    _b._check(st, "deer_sequential")
+    return {"z": out, "lam": lam, "grads": grads}
+
+
+def deer_sequential_workspace_bytes(model, B: int, T: int) -> int:
+    return int(load().deer_sequential_workspace_bytes(ctypes.byref(_model(model).c), B, T))
 
 
 def plrnn_jacobian(model, x, z, alpha: float, n_forced: int, *, z0=None, want=("F", "r", "masks"),

@@ -81,6 +81,11 @@ def load(path: str = LIB_PATH):
     lib.deer_adjoint_ex.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, i32, vp, P(deer_grads),
                                     vp, sz, vp]
     lib.deer_adjoint_ex.restype = i32
+    lib.deer_sequential.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, vp, P(deer_grads), vp,
+                                    sz, vp]
+    lib.deer_sequential.restype = i32
+    lib.deer_sequential_workspace_bytes.argtypes = [P(deer_model), i32, i32]
+    lib.deer_sequential_workspace_bytes.restype = sz
     lib.deer_readout_workspace_bytes.argtypes = [P(deer_readout), i32, i32, i32]
     lib.deer_readout_workspace_bytes.restype = sz
     lib.deer_readout_loss.argtypes = [P(deer_readout), i32, i32, i32, vp, vp, vp, vp, vp, P(deer_readout_grads), vp,

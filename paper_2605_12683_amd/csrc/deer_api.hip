@@ -935,6 +935,42 @@ static int check_readout(const deer_readout *r, int B, int T, int M) {
     return DEER_OK;
 }
 
+// ---- sequential baseline -------------------------------------------------------------------
+static int check_sequential(const deer_model *m, const deer_forcing *f, int B, int T, SeqArgs *a) {
+    if (!m || !f) { set_error("model/forcing pointer is NULL"); return DEER_ERR_INVALID_ARG; }
+    if (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN) {
+        set_error("the sequential baseline covers the PLRNN kinds");
+        return DEER_ERR_INVALID_ARG;
+    }
+    if (B <= 0 || T <= 0) { set_error("B and T must be positive (B=%d, T=%d)", B, T); return DEER_ERR_INVALID_ARG; }
+    if (!(f->alpha >= 0.0f && f->alpha <= 1.0f)) { set_error("alpha must lie in [0, 1]"); return DEER_ERR_INVALID_ARG; }
+    if (m->M <= 0 || f->n_forced < 0 || f->n_forced > m->M) {
+        set_error("need M >= 1 and 0 <= n_forced <= M");
+        return DEER_ERR_INVALID_ARG;
+    }
+    if (!m->A || !m->W || (m->kind == DEER_SHPLRNN && (!m->W2 || m->L <= 0))) {
+        set_error("model parameters A, W (and W2, L for the shallow kind) are required");
+        return DEER_ERR_INVALID_ARG;
+    }
+    const bool sh = m->kind == DEER_SHPLRNN;
+    const int L = sh ? m->L : m->M;
+    if (seq_check(m->M, L, sh)) {
+        set_error("the sequential baseline supports M, L <= 256 and M L <= 8192 (M=%d, L=%d)", m->M, L);
+        return DEER_ERR_INVALID_ARG;
+    }
+    if ((long)B * (long)T * (m->M > L ? m->M : L) >= (1L << 31)) { set_error("B*T too large"); return DEER_ERR_INVALID_ARG; }
+    *a = SeqArgs{m->A, m->W, sh ? m->W2 : nullptr, m->h, sh ? m->h2 : nullptr, f->alpha, f->n_forced, nullptr,
+                 nullptr, B, T, m->M, L, sh};
+    return DEER_OK;
+}
+
+static void carve_seq(void *ws, const SeqArgs &a, float **act, float **part, size_t *bytes) {
+    Carver c(ws);
+    *act = a.sh ? c.take<float>((size_t)a.B * a.T * a.L) : nullptr;
+    *part = c.take<float>((size_t)a.B * seq_part_floats(a.M, a.L, a.sh));
+    *bytes = c.off;
+}
+
 size_t deer_readout_workspace_bytes(const deer_readout *r, int B, int T, int M) {
     if (check_readout(r, B, T, M) != DEER_OK) return 0;
     return readout_ws_bytes(B, T);
@@ -980,6 +1016,38 @@ int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, cons
     }
     set_error("deer_scan: unknown layout %d", layout);
     return DEER_ERR_INVALID_ARG;
+}
+
+size_t deer_sequential_workspace_bytes(const deer_model *m, int B, int T) {
+    deer_forcing f{0.f, 0};
+    SeqArgs a{};
+    if (check_sequential(m, &f, B, T, &a)) return 0;
+    float *act = nullptr, *part = nullptr;
+    size_t need = 0;
+    carve_seq(nullptr, a, &act, &part, &need);
+    return need;
+}
+
+int deer_sequential(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0, float *z,
+                    const float *g, float *lam, const deer_grads *grads, void *ws, size_t ws_bytes, void *stream) {
+    set_error("");
+    SeqArgs a{};
+    int rc = check_sequential(m, f, B, T, &a);
+    if (rc) return rc;
+    if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
+    a.x = x;
+    a.z0 = z0;
+    float *act = nullptr, *part = nullptr;
+    size_t need = 0;
+    carve_seq(nullptr, a, &act, &part, &need);
+    if ((rc = check_ws(ws, ws_bytes, need))) return rc;
+    carve_seq(ws, a, &act, &part, &need);
+    hipStream_t st = (hipStream_t)stream;
+    const bool back = lam || (grads && (grads->A || grads->W || grads->W2 || grads->h || grads->h2));
+    if ((rc = launch_seq_forward(a, z, back ? act : nullptr, st))) return rc;
+    if (!back) return DEER_OK;
+    const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
+    return launch_seq_backward(a, z, act, g, scale, lam, part, grads, st);
 }
 
 }  // extern "C"

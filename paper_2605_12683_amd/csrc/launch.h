@@ -141,6 +141,21 @@ size_t diag_adjoint_ws_bytes(int B, int T, int M, int K);
 int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const float *g, bool g_real, const float *h,
                         const float *x, float *lam_out, float *dlam, float *dBc, void *ws, hipStream_t st);
 
+// sequential baseline (k_seq.hip): one workgroup per sequence, the steps in order
+struct SeqArgs {
+    const float *A, *W1, *W2, *h1, *h2;   // vanilla: W1 = W (M x M), W2 = h2 = null, L = M
+    float alpha;
+    int N;
+    const float *x, *z0;
+    int B, T, M, L;
+    bool sh;
+};
+int seq_check(int M, int L, bool sh);
+size_t seq_part_floats(int M, int L, bool sh);
+int launch_seq_forward(const SeqArgs &a, float *z, float *act, hipStream_t st);
+int launch_seq_backward(const SeqArgs &a, const float *z, const float *act, const float *g, float seed_scale,
+                        float *lam, float *part, const deer_grads *gr, hipStream_t st);
+
 // small utilities
 int launch_fill_teacher(int B, int T, int M, int N, const float *x, float *z, hipStream_t st);
 int launch_fill_i32(int *p, int n, int v, hipStream_t st);

@@ -195,6 +195,69 @@ def cpu_baseline(c, budget_s=20.0):
             "seconds": dt, "host_cpus": os.cpu_count()}
 
 
+def fig1a_sweep(reps: int = 3):
+    """Runtime of one training step (forward + backward with the parameter gradients), GTF-DEER
+    against the sequential baseline on the same GPU, over the grid of Fig. 1A: shallow PLRNN
+    L = 50, M in (4, 16, 64, 128), B = 1, T = 2^7 ... 2^15, alpha = 0.15, Lorenz-63 data (N = 3).
+    Models are not trained: "random" draws the default initialisation (A in [0.5, 0.95], W1, W2
+    with variance 1/L), which is not a contraction for M >= 16 and makes DEER take many Newton
+    updates; "contracting" rescales W1 so that max A + ||W1|| ||W2|| < 1 (A in [0.5, 0.65],
+    ||W1|| ||W2|| = 0.3), the regime GTF is meant to produce.  DEER's iteration counts are those
+    of the model at hand.  The parallel solver covers M <= 64.  One JSON line per point."""
+    import torch
+    import workloads as W
+    import paper_2605_12683_amd as D
+
+    L, N, alpha = 50, 3, 0.15
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            out = fn()
+            torch.cuda.synchronize()
+            ts.append(time.perf_counter() - t0)
+        return float(np.median(ts)) * 1e3, out
+
+    for init in ("random", "contracting"):
+        for M in (4, 16, 64, 128):
+            _fig1a_model(D, W, init, M, L, N, alpha, timed)
+
+
+def _fig1a_model(D, W, init, M, L, N, alpha, timed):
+    import torch
+    rng = np.random.default_rng(9000 + M)
+    if init == "random":
+        params = W.shplrnn_params(M, L, rng)
+    else:
+        params = W.shplrnn_params(M, L, rng, a_range=(0.5, 0.65))
+        W1 = params["W1"].astype(np.float64)
+        norm = np.linalg.norm(W1, 2) * np.linalg.norm(params["W2"].astype(np.float64), 2)
+        params["W1"] = (W1 * (0.3 / norm)).astype(np.float32)
+    model = D._Model({"kind": "shplrnn", **params})
+    for lt in range(7, 16):
+        T = 1 << lt
+        x = torch.tensor(W.observed_batch("lorenz63", N, 1, T, 9100 + lt), device="cuda")
+        ws_q = D._workspace(D.deer_sequential_workspace_bytes(model, 1, T))
+        seq_ms, _ = timed(lambda: D.deer_sequential(model, x, alpha, N, ws=ws_q, want_lam=False))
+        rec = {"sweep": "fig1a", "model": "shplrnn", "init": init, "M": M, "L": L, "B": 1, "T": T, "alpha": alpha,
+               "sequential_ms": round(seq_ms, 4), "deer_ms": None, "newton_updates": None, "speedup": None}
+        if M <= 64:
+            ws_s = D._workspace(D.deer_workspace_bytes(model, 1, T, 0))
+            ws_a = D._workspace(D.deer_workspace_bytes(model, 1, T, 1))
+
+            def step():
+                r = D.deer_solve(model, x, alpha, N, tol=1e-5, max_iter=500, ws=ws_s, check=False)
+                D.deer_adjoint(model, x, r["z"], alpha, N, ws=ws_a, want_lam=False)
+                return r
+            deer_ms, r = timed(step)
+            rec.update(deer_ms=round(deer_ms, 4), newton_updates=int(sum(r["iters"])),
+                       speedup=round(seq_ms / deer_ms, 3), status=int(r["status"]))
+        print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,11 +265,16 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--fig1a", action="store_true",
+                    help="instead of the workload: the Fig. 1A sweep, GTF-DEER against the sequential baseline")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
               file=sys.stderr)
         sys.exit(2)
+    if args.fig1a:
+        fig1a_sweep()
+        return
 
     import torch
     import workloads as W

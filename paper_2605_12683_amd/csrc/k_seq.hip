@@ -1,7 +1,11 @@
 // Sequential GTF baseline: the forward rollout z_s = F(z~_s) step by step and back-propagation
 // through time, also step by step (the training the parallel solver replaces; the comparison
-// of Fig. 1A).  One workgroup of 256 threads per sequence, weights in LDS, the steps in order:
-// the batch is the only parallel dimension, as in a sequential scan vectorised over sequences.
+// of Fig. 1A).  One wave per sequence, the batch being the only parallel dimension, as in a
+// sequential scan vectorised over sequences.  A wave needs no workgroup barrier: its lanes
+// exchange data through LDS, synchronised within the wave.  Weights live in LDS; the per-step
+// inputs (x, and for the backward pass z, g and the hidden activations) are staged into LDS a
+// chunk of steps at a time, so the loop does not wait for memory at every step; the outer-
+// product gradient sums are formed per chunk from buffered (lambda, a) and (q, z~) rows.
 //
 // Model (both PLRNN kinds; the vanilla one is the shallow form with u = z~, L = M):
 //   z~_s = z0 (or [x_0; 0]) at s = 0, else fl(fl(p z_{s-1}) + fl(alpha x_s)) on the forced
@@ -19,14 +23,31 @@ namespace deer {
 
 namespace {
 
-constexpr int kSeqThreads = 256;
-constexpr int kSeqAcc = 32;   // gradient entries per thread and matrix: M L <= 256 * 32
+constexpr int kW = 64;                  // one wave per sequence
+constexpr int kSeqMaxDim = 256;         // M, L <= 256: at most four outputs per lane
+constexpr int kNQ = kSeqMaxDim / kW;
+constexpr size_t kSeqLdsFloats = 38 * 1024;   // LDS budget of a sequence (152 KiB)
 
 __device__ __forceinline__ float pforce(int i, int N, float alpha) { return i < N ? __fsub_rn(1.0f, alpha) : 1.0f; }
 
-// weights into LDS: W1 [M][L+1], W2 [L][M+1] (padded rows), A, h1 [M], h2 [L]
+// sum_k w[k * stride] v[k], k < n, in four interleaved partial sums (short dependency chains)
+__device__ __forceinline__ float seq_dot(const float *w, int stride, const float *v, int n) {
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    int k = 0;
+    for (; k + 4 <= n; k += 4) {
+        a0 = fmaf(w[(size_t)k * stride], v[k], a0);
+        a1 = fmaf(w[(size_t)(k + 1) * stride], v[k + 1], a1);
+        a2 = fmaf(w[(size_t)(k + 2) * stride], v[k + 2], a2);
+        a3 = fmaf(w[(size_t)(k + 3) * stride], v[k + 3], a3);
+    }
+    for (; k < n; ++k) a0 = fmaf(w[(size_t)k * stride], v[k], a0);
+    return (a0 + a1) + (a2 + a3);
+}
+
+// LDS: W1 [M][L+1], W2 [L][M+1], A, h1 [M], h2 [L], zt [M], a [L], lam [M], q [L], then the
+// chunk buffers
 struct SeqLds {
-    float *W1, *W2, *A, *h1, *h2, *zt, *a, *lam, *q;
+    float *W1, *W2, *A, *h1, *h2, *zt, *a, *lam, *q, *buf;
 };
 __device__ __forceinline__ SeqLds seq_lds(float *sm, int M, int L, bool sh) {
     SeqLds s;
@@ -39,27 +60,42 @@ __device__ __forceinline__ SeqLds seq_lds(float *sm, int M, int L, bool sh) {
     s.a = s.zt + M;
     s.lam = s.a + L;
     s.q = s.lam + M;
+    s.buf = s.q + L;
     return s;
 }
+__host__ __device__ inline size_t seq_fixed_floats(int M, int L, bool sh) {
+    return (size_t)M * (L + 1) + (sh ? (size_t)L * (M + 1) : 0) + 4 * (size_t)M + 4 * (size_t)L;
+}
+// floats a chunk step needs: forward x rows; backward z, x, g and a rows and the lam, z~, a, q
+// rows of the gradient sums (plus one more z and x row per chunk)
+__host__ __device__ inline size_t seq_step_floats(int M, int L, int N, bool sh, bool has_g, bool backward) {
+    return backward ? (size_t)M + N + (has_g ? M : 0) + (sh ? L : 0) + 2 * (size_t)(M + L) : (size_t)(N > 0 ? N : 1);
+}
+__host__ __device__ inline int seq_chunk(int M, int L, int N, bool sh, bool has_g, bool backward) {
+    const size_t fixed = seq_fixed_floats(M, L, sh) + (backward ? (size_t)M + N : 0);
+    if (fixed + 64 > kSeqLdsFloats) return 0;
+    size_t ch = (kSeqLdsFloats - fixed) / seq_step_floats(M, L, N, sh, has_g, backward);
+    if (ch > 256) ch = 256;
+    return (int)ch;
+}
+
 __device__ __forceinline__ void seq_load_weights(const SeqLds &s, const float *A, const float *W1, const float *W2,
-                                                 const float *h1, const float *h2, int M, int L, bool sh) {
-    for (int e = threadIdx.x; e < M * L; e += blockDim.x) s.W1[(e / L) * (L + 1) + e % L] = W1[e];
+                                                 const float *h1, const float *h2, int M, int L, bool sh, int lane) {
+    for (int e = lane; e < M * L; e += kW) s.W1[(e / L) * (L + 1) + e % L] = W1[e];
     if (sh)
-        for (int e = threadIdx.x; e < L * M; e += blockDim.x) s.W2[(e / M) * (M + 1) + e % M] = W2[e];
-    for (int i = threadIdx.x; i < M; i += blockDim.x) {
+        for (int e = lane; e < L * M; e += kW) s.W2[(e / M) * (M + 1) + e % M] = W2[e];
+    for (int i = lane; i < M; i += kW) {
         s.A[i] = A[i];
         s.h1[i] = h1 ? h1[i] : 0.f;
     }
-    if (sh)
-        for (int l = threadIdx.x; l < L; l += blockDim.x) s.h2[l] = h2 ? h2[l] : 0.f;
+    for (int l = lane; l < L; l += kW) s.h2[l] = (sh && h2) ? h2[l] : 0.f;
 }
 
-// u_l = h2_l + sum_j W2[l][j] z~_j (left to right, rounded after every operation)
-__device__ __forceinline__ float seq_pre(const SeqLds &s, int l, int M) {
-    float u = s.h2[l];
-    const float *w = s.W2 + (size_t)l * (M + 1);
-    for (int j = 0; j < M; ++j) u = __fadd_rn(u, __fmul_rn(w[j], s.zt[j]));
-    return u;
+// rows [r0, r0 + n) of a row-major array of width w into LDS, lanes striding
+__device__ __forceinline__ void seq_stage(float *dst, const float *src, size_t r0, int n, int w, int lane) {
+    const size_t cnt = (size_t)n * w;
+    const float *p = src + r0 * w;
+    for (size_t e = lane; e < cnt; e += kW) dst[e] = p[e];
 }
 
 }  // namespace
@@ -67,50 +103,72 @@ __device__ __forceinline__ float seq_pre(const SeqLds &s, int l, int M) {
 // Forward rollout.  act (shallow, may be null) receives a_s = relu(u_s) [B][T][L] for the
 // backward pass.
 template <bool SH>
-__global__ __launch_bounds__(kSeqThreads) void k_seq_forward(const float *__restrict__ A, const float *__restrict__ W1,
-                                                             const float *__restrict__ W2, const float *__restrict__ h1,
-                                                             const float *__restrict__ h2, float alpha, int N,
-                                                             const float *__restrict__ x, const float *__restrict__ z0,
-                                                             float *__restrict__ z, float *__restrict__ act, int T,
-                                                             int M, int L) {
+__global__ __launch_bounds__(kW) void k_seq_forward(const float *__restrict__ A, const float *__restrict__ W1,
+                                                    const float *__restrict__ W2, const float *__restrict__ h1,
+                                                    const float *__restrict__ h2, float alpha, int N,
+                                                    const float *__restrict__ x, const float *__restrict__ z0,
+                                                    float *__restrict__ z, float *__restrict__ act, int T, int M,
+                                                    int L, int CH) {
     extern __shared__ float sm[];
+    const int lane = threadIdx.x, b = blockIdx.x;
     const SeqLds s = seq_lds(sm, M, L, SH);
-    seq_load_weights(s, A, W1, W2, h1, h2, M, L, SH);
-    const int b = blockIdx.x, tid = threadIdx.x;
+    seq_load_weights(s, A, W1, W2, h1, h2, M, L, SH, lane);
     const float *xb = x + (size_t)b * (T + 1) * N;
     float *zb = z + (size_t)b * T * M;
-    float zprev = 0.f;   // z_{s-1} of latent tid (the initial state at s = 0)
-    if (tid < M) zprev = z0 ? z0[(size_t)b * M + tid] : (tid < N ? xb[tid] : 0.f);
-    const float pi = pforce(tid, N, alpha);
-    __syncthreads();
-    for (int s0 = 0; s0 < T; ++s0) {
-        float zt = 0.f;
-        if (tid < M) {
-            zt = (s0 == 0 || tid >= N) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xb[(size_t)s0 * N + tid]));
-            s.zt[tid] = zt;
-        }
-        __syncthreads();
-        if (SH) {
-            for (int l = tid; l < L; l += kSeqThreads) {
-                const float u = seq_pre(s, l, M);
-                const float av = u > 0.f ? u : 0.f;
-                s.a[l] = av;
-                if (act) act[((size_t)b * T + s0) * L + l] = av;
+    float *xs = s.buf;   // x rows of the chunk [CH][N]
+    float zprev[kNQ];    // z_{s-1} of latents lane + 64 r
+#pragma unroll
+    for (int r = 0; r < kNQ; ++r) {
+        const int i = lane + kW * r;
+        zprev[r] = i < M ? (z0 ? z0[(size_t)b * M + i] : (i < N ? xb[i] : 0.f)) : 0.f;
+    }
+    for (int c0 = 0; c0 < T; c0 += CH) {
+        const int n = min(CH, T - c0);
+        wave_lds_sync();
+        if (N > 0) seq_stage(xs, xb, c0, n, N, lane);
+        wave_lds_sync();
+        for (int t = 0; t < n; ++t) {
+            const int s0 = c0 + t;
+            float zt[kNQ];
+#pragma unroll
+            for (int r = 0; r < kNQ; ++r) {
+                const int i = lane + kW * r;
+                zt[r] = 0.f;
+                if (i < M) {
+                    zt[r] = (s0 == 0 || i >= N) ? zprev[r]
+                                                : __fadd_rn(__fmul_rn(pforce(i, N, alpha), zprev[r]),
+                                                            __fmul_rn(alpha, xs[(size_t)t * N + i]));
+                    s.zt[i] = zt[r];
+                }
             }
-        } else if (tid < M) {
-            s.a[tid] = zt > 0.f ? zt : 0.f;
+            wave_lds_sync();
+            if (SH) {
+                for (int l = lane; l < L; l += kW) {
+                    float u = s.h2[l];
+                    const float *w = s.W2 + (size_t)l * (M + 1);
+                    for (int j = 0; j < M; ++j) u = __fadd_rn(u, __fmul_rn(w[j], s.zt[j]));
+                    const float av = u > 0.f ? u : 0.f;
+                    s.a[l] = av;
+                    if (act) act[((size_t)b * T + s0) * L + l] = av;
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < kNQ; ++r) {
+                    const int i = lane + kW * r;
+                    if (i < M) s.a[i] = zt[r] > 0.f ? zt[r] : 0.f;
+                }
+            }
+            wave_lds_sync();
+#pragma unroll
+            for (int r = 0; r < kNQ; ++r) {
+                const int i = lane + kW * r;
+                if (i < M) {
+                    const float F = fmaf(s.A[i], zt[r], seq_dot(s.W1 + (size_t)i * (L + 1), 1, s.a, L)) + s.h1[i];
+                    zb[(size_t)s0 * M + i] = F;
+                    zprev[r] = F;
+                }
+            }
         }
-        __syncthreads();
-        if (tid < M) {
-            const float *w = s.W1 + (size_t)tid * (L + 1);
-            float acc = 0.f;
-            for (int k = 0; k < L; ++k) acc = fmaf(w[k], s.a[k], acc);
-            const float F = fmaf(s.A[tid], zt, acc) + s.h1[tid];
-            zb[(size_t)s0 * M + tid] = F;
-            zprev = F;
-        }
-        // the next step writes zt only: every thread has passed the barrier after this
-        // step's a, and a is written again only after the next barrier
     }
 }
 
@@ -118,112 +176,135 @@ __global__ __launch_bounds__(kSeqThreads) void k_seq_forward(const float *__rest
 // x_{s+1}; 0].  lam (may be null) receives lam_s.  part receives the sequence's gradient sums
 // [A M | W1 M L | h1 M | W2 L M | h2 L] (shallow) or [A M | W M M | h M] (vanilla).
 template <bool SH>
-__global__ __launch_bounds__(kSeqThreads) void k_seq_backward(
+__global__ __launch_bounds__(kW) void k_seq_backward(
     const float *__restrict__ A, const float *__restrict__ W1, const float *__restrict__ W2,
     const float *__restrict__ h1, const float *__restrict__ h2, float alpha, int N, const float *__restrict__ x,
     const float *__restrict__ z0, const float *__restrict__ z, const float *__restrict__ act,
     const float *__restrict__ g, float seed_scale, float *__restrict__ lam, float *__restrict__ part, int T, int M,
-    int L) {
+    int L, int CH) {
     extern __shared__ float sm[];
+    const int lane = threadIdx.x, b = blockIdx.x;
     const SeqLds s = seq_lds(sm, M, L, SH);
-    seq_load_weights(s, A, W1, W2, h1, h2, M, L, SH);
-    const int b = blockIdx.x, tid = threadIdx.x;
+    seq_load_weights(s, A, W1, W2, h1, h2, M, L, SH, lane);
     const float *xb = x + (size_t)b * (T + 1) * N;
     const float *zb = z + (size_t)b * T * M;
-    const float pi = pforce(tid, N, alpha);
     const int ML = M * L;
-    // this thread's entries of the two outer-product sums: e = tid + 256 q of W1 (row-major M x L,
-    // packed i << 16 | k) and of W2 (row-major L x M)
-    uint32_t e1[kSeqAcc], e2[kSeqAcc];
-    float g1[kSeqAcc], g2[kSeqAcc];
-#pragma unroll
-    for (int q = 0; q < kSeqAcc; ++q) {
-        const int e = tid + kSeqThreads * q;
-        e1[q] = e < ML ? ((uint32_t)(e / L) << 16) | (uint32_t)(e % L) : 0xffffffffu;
-        e2[q] = (SH && e < ML) ? ((uint32_t)(e / M) << 16) | (uint32_t)(e % M) : 0xffffffffu;
-        g1[q] = 0.f;
-        g2[q] = 0.f;
-    }
-    float gA = 0.f, gh1 = 0.f, gh2 = 0.f;
-    // z~_s of latent tid
-    auto forced = [&](int s0) {
-        if (tid >= M) return 0.f;
-        if (s0 == 0) return z0 ? z0[(size_t)b * M + tid] : (tid < N ? xb[tid] : 0.f);
-        const float zp = zb[(size_t)(s0 - 1) * M + tid];
-        return tid >= N ? zp : __fadd_rn(__fmul_rn(pi, zp), __fmul_rn(alpha, xb[(size_t)s0 * N + tid]));
-    };
-    // q = m (W1^T lam) for the lam and a in LDS, into s.q (L entries); the W2 and h2 sums of the
-    // step whose z~ is in s.zt
-    auto backprop_hidden = [&]() {
-        for (int k = tid; k < L; k += kSeqThreads) {
-            float v = 0.f;
-            for (int i = 0; i < M; ++i) v = fmaf(s.W1[(size_t)i * (L + 1) + k], s.lam[i], v);
-            s.q[k] = s.a[k] > 0.f ? v : 0.f;
-        }
-        __syncthreads();
-        if (SH) {
-            for (int l = tid; l < L; l += kSeqThreads) gh2 += s.q[l];
-#pragma unroll
-            for (int qq = 0; qq < kSeqAcc; ++qq)
-                if (e2[qq] != 0xffffffffu) g2[qq] = fmaf(s.q[e2[qq] >> 16], s.zt[e2[qq] & 0xffffu], g2[qq]);
-        }
-    };
-    for (int s0 = T - 1; s0 >= 0; --s0) {
-        // lam_s = g_s + P (A lam_{s+1} + J^T part), with s.q = m_{s+1} (W1^T lam_{s+1})
-        if (s0 < T - 1) backprop_hidden();
-        float ls = 0.f, zt = 0.f;
-        if (tid < M) {
-            const float zs = zb[(size_t)s0 * M + tid];
-            float gs;
-            if (g) gs = g[((size_t)b * T + s0) * M + tid];
-            else gs = tid < N ? seed_scale * (zs - xb[(size_t)(s0 + 1) * N + tid]) : 0.f;
-            ls = gs;
-            if (s0 < T - 1) {
-                float w;
-                if (SH) {
-                    w = 0.f;
-                    for (int k = 0; k < L; ++k) w = fmaf(s.W2[(size_t)k * (M + 1) + tid], s.q[k], w);
-                } else {
-                    w = s.q[tid];
-                }
-                ls = fmaf(pi, fmaf(s.A[tid], s.lam[tid], w), gs);
-            }
-            zt = forced(s0);
-        }
-        __syncthreads();   // every read of lam_{s+1}, q and the previous z~, a is done
-        if (tid < M) {
-            s.lam[tid] = ls;
-            s.zt[tid] = zt;
-            if (lam) lam[((size_t)b * T + s0) * M + tid] = ls;
-            gA = fmaf(ls, zt, gA);
-            gh1 += ls;
-            if (!SH) s.a[tid] = zt > 0.f ? zt : 0.f;
-        }
-        if (SH)
-            for (int l = tid; l < L; l += kSeqThreads) s.a[l] = act[((size_t)b * T + s0) * L + l];
-        __syncthreads();
-        // dW1 += lam_s a_s^T
-#pragma unroll
-        for (int qq = 0; qq < kSeqAcc; ++qq)
-            if (e1[qq] != 0xffffffffu) g1[qq] = fmaf(s.lam[e1[qq] >> 16], s.a[e1[qq] & 0xffffu], g1[qq]);
-        __syncthreads();
-    }
-    backprop_hidden();   // the W2 and h2 sums of step 0
-    // this sequence's sums
     float *pA = part + (size_t)b * (SH ? (size_t)2 * M + 2 * (size_t)ML + L : (size_t)2 * M + ML);
     float *pW1 = pA + M, *ph1 = pW1 + ML, *pW2 = ph1 + M, *ph2 = pW2 + ML;
-    if (tid < M) {
-        pA[tid] = gA;
-        ph1[tid] = gh1;
+    for (int e = lane; e < ML; e += kW) {
+        pW1[e] = 0.f;
+        if (SH) pW2[e] = 0.f;
+    }
+    // chunk buffers: z rows c0-1 .. c1-1, x rows c0 .. c1, g and a rows c0 .. c1-1, then the
+    // rows of the gradient sums (lam, z~, a, q per step of the chunk)
+    float *zs = s.buf;                              // [CH + 1][M], row 0 = z_{c0-1}
+    float *xs = zs + (size_t)(CH + 1) * M;          // [CH + 1][N], row 0 = x_{c0}
+    float *gs = xs + (size_t)(CH + 1) * N;          // [CH][M] if g
+    float *as = gs + (g ? (size_t)CH * M : 0);      // [CH][L] shallow
+    float *rl = as + (SH ? (size_t)CH * L : 0);     // lam rows [CH][M]
+    float *rz = rl + (size_t)CH * M;                // z~ rows [CH][M]
+    float *ra = rz + (size_t)CH * M;                // a rows [CH][L]
+    float *rq = ra + (size_t)CH * L;                // q rows [CH][L]
+    float gA[kNQ], gh1[kNQ], gh2[kNQ];
+#pragma unroll
+    for (int r = 0; r < kNQ; ++r) gA[r] = gh1[r] = gh2[r] = 0.f;
+    bool first = true;   // s = T - 1: lam = g
+    for (int c1 = T; c1 > 0; c1 -= CH) {
+        const int c0 = max(0, c1 - CH), n = c1 - c0;
+        wave_lds_sync();
+        if (c0 > 0) seq_stage(zs, zb, c0 - 1, n + 1, M, lane);
+        else seq_stage(zs + M, zb, 0, n, M, lane);
+        if (N > 0) seq_stage(xs, xb, c0, n + 1, N, lane);
+        if (g) seq_stage(gs, g + (size_t)b * T * M, c0, n, M, lane);
+        if (SH) seq_stage(as, act + (size_t)b * T * L, c0, n, L, lane);
+        wave_lds_sync();
+        for (int t = n - 1; t >= 0; --t) {
+            const int s0 = c0 + t;
+            // lam_s = g_s + P (A lam_{s+1} + W2^T q_{s+1}), z~_s, a_s
+            float ls[kNQ], zt[kNQ];
+#pragma unroll
+            for (int r = 0; r < kNQ; ++r) {
+                const int i = lane + kW * r;
+                ls[r] = zt[r] = 0.f;
+                if (i >= M) continue;
+                const float gv = g ? gs[(size_t)t * M + i]
+                                   : (i < N ? seed_scale * (zs[(size_t)(t + 1) * M + i] - xs[(size_t)(t + 1) * N + i])
+                                            : 0.f);
+                ls[r] = gv;
+                if (!first) {
+                    const float w = SH ? seq_dot(s.W2 + i, M + 1, s.q, L) : s.q[i];
+                    ls[r] = fmaf(pforce(i, N, alpha), fmaf(s.A[i], s.lam[i], w), gv);
+                }
+                if (s0 == 0) {
+                    zt[r] = z0 ? z0[(size_t)b * M + i] : (i < N ? xb[i] : 0.f);
+                } else {
+                    const float zp = zs[(size_t)t * M + i];
+                    zt[r] = i >= N ? zp
+                                   : __fadd_rn(__fmul_rn(pforce(i, N, alpha), zp), __fmul_rn(alpha, xs[(size_t)t * N + i]));
+                }
+            }
+            first = false;
+            wave_lds_sync();   // every read of lam_{s+1} and q_{s+1} is done
+#pragma unroll
+            for (int r = 0; r < kNQ; ++r) {
+                const int i = lane + kW * r;
+                if (i >= M) continue;
+                s.lam[i] = ls[r];
+                s.zt[i] = zt[r];
+                rl[(size_t)t * M + i] = ls[r];
+                rz[(size_t)t * M + i] = zt[r];
+                if (lam) lam[((size_t)b * T + s0) * M + i] = ls[r];
+                gA[r] = fmaf(ls[r], zt[r], gA[r]);
+                gh1[r] += ls[r];
+                if (!SH) {
+                    const float av = zt[r] > 0.f ? zt[r] : 0.f;
+                    s.a[i] = av;
+                    ra[(size_t)t * L + i] = av;
+                }
+            }
+            if (SH)
+                for (int l = lane; l < L; l += kW) {
+                    const float av = as[(size_t)t * L + l];
+                    s.a[l] = av;
+                    ra[(size_t)t * L + l] = av;
+                }
+            wave_lds_sync();
+            // q_s = m_s (W1^T lam_s): the next step's W2^T q and this step's W2, h2 sums
+#pragma unroll
+            for (int r = 0; r < kNQ; ++r) {
+                const int k = lane + kW * r;
+                if (k >= L) continue;
+                const float v = seq_dot(s.W1 + k, L + 1, s.lam, M);
+                const float qv = s.a[k] > 0.f ? v : 0.f;
+                s.q[k] = qv;
+                rq[(size_t)t * L + k] = qv;
+                gh2[r] += qv;
+            }
+            wave_lds_sync();
+        }
+        // the chunk's outer-product sums: W1 += sum_t lam_t a_t^T, W2 += sum_t q_t z~_t^T
+        for (int e = lane; e < ML; e += kW) {
+            const int i = e / L, k = e - i * L;
+            float acc = 0.f;
+            for (int t = 0; t < n; ++t) acc = fmaf(rl[(size_t)t * M + i], ra[(size_t)t * L + k], acc);
+            pW1[e] += acc;
+            if (SH) {
+                const int l = e / M, j = e - l * M;
+                float acc2 = 0.f;
+                for (int t = 0; t < n; ++t) acc2 = fmaf(rq[(size_t)t * L + l], rz[(size_t)t * M + j], acc2);
+                pW2[e] += acc2;
+            }
+        }
     }
 #pragma unroll
-    for (int qq = 0; qq < kSeqAcc; ++qq) {
-        const int e = tid + kSeqThreads * qq;
-        if (e < ML) pW1[e] = g1[qq];
-        if (SH && e < ML) pW2[e] = g2[qq];
+    for (int r = 0; r < kNQ; ++r) {
+        const int i = lane + kW * r;
+        if (i < M) {
+            pA[i] = gA[r];
+            ph1[i] = gh1[r];
+        }
+        if (SH && i < L) ph2[i] = gh2[r];
     }
-    if (SH)
-        for (int l = tid; l < L; l += kSeqThreads) ph2[l] = gh2;
 }
 
 // sum over the B sequences' parts (float64), into the gradient outputs
@@ -247,61 +328,60 @@ __global__ void k_seq_grads_sum(const float *__restrict__ part, int B, int M, in
     }
 }
 
-size_t seq_lds_bytes(int M, int L, bool sh) {
-    return sizeof(float) * ((size_t)M * (L + 1) + (sh ? (size_t)L * (M + 1) : 0) + 3 * (size_t)M + 3 * (size_t)L + M);
-}
-
 size_t seq_part_floats(int M, int L, bool sh) {
     return sh ? (size_t)2 * M + 2 * (size_t)M * L + L : (size_t)2 * M + (size_t)M * L;
 }
 
 int seq_check(int M, int L, bool sh) {
-    if (M > kSeqThreads || (sh && L > kSeqThreads) || (size_t)M * L > (size_t)kSeqThreads * kSeqAcc ||
-        seq_lds_bytes(M, L, sh) > 160 * 1024)
-        return -1;
+    if (M > kSeqMaxDim || L > kSeqMaxDim || (size_t)M * L > 8192) return -1;
+    // the largest stage: backward with a cotangent and the largest forcing count N = M
+    if (seq_chunk(M, L, M, sh, true, true) < 8) return -1;
     return 0;
 }
 
 int launch_seq_forward(const SeqArgs &a, float *z, float *act, hipStream_t st) {
-    const size_t lds = seq_lds_bytes(a.M, a.L, a.sh);
+    const int CH = seq_chunk(a.M, a.L, a.N, a.sh, false, false);
+    const size_t lds = sizeof(float) * (seq_fixed_floats(a.M, a.L, a.sh) +
+                                        (size_t)CH * seq_step_floats(a.M, a.L, a.N, a.sh, false, false));
     KTimer kt("k_seq_forward", st);
-    if (a.sh) {
-        DEER_HIP(hipFuncSetAttribute((const void *)k_seq_forward<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)lds));
-        hipLaunchKernelGGL(k_seq_forward<true>, dim3(a.B), dim3(kSeqThreads), lds, st, a.A, a.W1, a.W2, a.h1, a.h2,
-                           a.alpha, a.N, a.x, a.z0, z, act, a.T, a.M, a.L);
-    } else {
-        DEER_HIP(hipFuncSetAttribute((const void *)k_seq_forward<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)lds));
-        hipLaunchKernelGGL(k_seq_forward<false>, dim3(a.B), dim3(kSeqThreads), lds, st, a.A, a.W1, a.W2, a.h1, a.h2,
-                           a.alpha, a.N, a.x, a.z0, z, act, a.T, a.M, a.L);
-    }
+#define SEQF(SHV)                                                                                                  \
+    do {                                                                                                           \
+        DEER_HIP(hipFuncSetAttribute((const void *)k_seq_forward<SHV>, hipFuncAttributeMaxDynamicSharedMemorySize, \
+                                     (int)lds));                                                                   \
+        hipLaunchKernelGGL(k_seq_forward<SHV>, dim3(a.B), dim3(kW), lds, st, a.A, a.W1, a.W2, a.h1, a.h2, a.alpha, \
+                           a.N, a.x, a.z0, z, act, a.T, a.M, a.L, CH);                                             \
+    } while (0)
+    if (a.sh) SEQF(true);
+    else SEQF(false);
+#undef SEQF
     DEER_LAUNCH_CHECK("k_seq_forward");
     return DEER_OK;
 }
 
 int launch_seq_backward(const SeqArgs &a, const float *z, const float *act, const float *g, float seed_scale,
                         float *lam, float *part, const deer_grads *gr, hipStream_t st) {
-    const size_t lds = seq_lds_bytes(a.M, a.L, a.sh);
+    const bool hg = g != nullptr;
+    const int CH = seq_chunk(a.M, a.L, a.N, a.sh, hg, true);
+    const size_t lds = sizeof(float) * (seq_fixed_floats(a.M, a.L, a.sh) + (size_t)a.M + a.N +
+                                        (size_t)CH * seq_step_floats(a.M, a.L, a.N, a.sh, hg, true));
     {
         KTimer kt("k_seq_backward", st);
-        if (a.sh) {
-            DEER_HIP(hipFuncSetAttribute((const void *)k_seq_backward<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         (int)lds));
-            hipLaunchKernelGGL(k_seq_backward<true>, dim3(a.B), dim3(kSeqThreads), lds, st, a.A, a.W1, a.W2, a.h1,
-                               a.h2, a.alpha, a.N, a.x, a.z0, z, act, g, seed_scale, lam, part, a.T, a.M, a.L);
-        } else {
-            DEER_HIP(hipFuncSetAttribute((const void *)k_seq_backward<false>,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-            hipLaunchKernelGGL(k_seq_backward<false>, dim3(a.B), dim3(kSeqThreads), lds, st, a.A, a.W1, a.W2, a.h1,
-                               a.h2, a.alpha, a.N, a.x, a.z0, z, act, g, seed_scale, lam, part, a.T, a.M, a.L);
-        }
+#define SEQB(SHV)                                                                                                   \
+    do {                                                                                                            \
+        DEER_HIP(hipFuncSetAttribute((const void *)k_seq_backward<SHV>, hipFuncAttributeMaxDynamicSharedMemorySize, \
+                                     (int)lds));                                                                    \
+        hipLaunchKernelGGL(k_seq_backward<SHV>, dim3(a.B), dim3(kW), lds, st, a.A, a.W1, a.W2, a.h1, a.h2, a.alpha, \
+                           a.N, a.x, a.z0, z, act, g, seed_scale, lam, part, a.T, a.M, a.L, CH);                    \
+    } while (0)
+        if (a.sh) SEQB(true);
+        else SEQB(false);
+#undef SEQB
         DEER_LAUNCH_CHECK("k_seq_backward");
     }
     if (gr) {
         KTimer kt("k_seq_grads_sum", st);
-        const size_t per = seq_part_floats(a.M, a.L, a.sh);
-        const unsigned grid = (unsigned)((per + 255) / 256);
+        const size_t pf = seq_part_floats(a.M, a.L, a.sh);
+        const unsigned grid = (unsigned)((pf + 255) / 256);
         hipLaunchKernelGGL(k_seq_grads_sum, dim3(grid), dim3(256), 0, st, (const float *)part, a.B, a.M, a.L,
                            a.sh ? 1 : 0, *gr);
         DEER_LAUNCH_CHECK("k_seq_grads_sum");

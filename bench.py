@@ -70,6 +70,7 @@ def kernel_work(c, steps, updates):
             "k_diag_seg_write": ("hbm", elems * 8 + xin),
             # adjoint: real cotangent (4 B) and forward states (8 B) read, dlam / dBc accumulated
             # on the way (the training step does not store the adjoint itself)
+            "k_diag_rseg": ("hbm", elems * 12 + xin),
             "k_diag_scan_lb_grads": ("hbm", elems * 12 + xin),
             "k_diag_scan_lb": ("hbm", elems * 12 + xin),
             # read-out: three [rows x 64] x [64 x 128] products (s, g, dWa) on the matrix cores
@@ -112,7 +113,8 @@ def kernel_work(c, steps, updates):
 KERNEL_SOURCE = {"k_newton_product_plrnn": "k_plrnn.hip", "k_newton_pass16": "k_plrnn.hip", "k_chunk_product_plrnn": "k_plrnn.hip",
                  "k_fixup_fwd_plrnn": "k_plrnn.hip", "k_jacform_shplrnn": "k_shallow.hip",
                  "k_chunk_product_dense": "k_dense.hip", "k_readout": "k_readout.hip",
-                 "k_diag_scan_lb_grads": "k_diag.hip", "k_diag_seg_write": "k_diag.hip"}
+                 "k_diag_scan_lb_grads": "k_diag.hip", "k_diag_seg_write": "k_diag.hip",
+                 "k_diag_rseg": "k_diag.hip"}
 CALIB_COPY_BYTES = 256 << 20
 
 

@@ -14,6 +14,8 @@
 // the fly as b_t = Bc u_t with u_t = x_{t-1} (input projection fused, K inputs).
 #include <stdlib.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 
@@ -539,14 +541,19 @@ __global__ __launch_bounds__(256) void k_diag_seg(const float *__restrict__ lam,
 }
 
 // carry[s] = state at the end of segment s - 1:  X_0 = 0,  X_{s+1} = Lambda X_s + A_s,
-// Lambda = lam^SEG (every segment but the last is full; the last aggregate is not needed).
+// Lambda = lam^seglen (conj(lam) for a reverse scan; every segment but the last is full, and
+// the last aggregate is not needed).
 // Block = (sequence, 64-channel tile), threads = (group g of CG consecutive segments, channel):
 // group aggregates, a sequential pass over the 16 groups, then every group re-walked from its
-// carry.  Serial depth 2 CG + 16 instead of nseg.
+// carry.  Serial depth 2 CG + 16 instead of nseg; the aggregates of a group are loaded
+// SEG_CB at a time (indices clamped to the group, so the loads are unconditional) before the
+// dependent float64 updates, so the walks wait on memory once per batch rather than once per
+// segment.
 constexpr int SEG_NG = 16;
+constexpr int SEG_CB = 16;
 
-__global__ __launch_bounds__(1024) void k_diag_seg_carry(const float *__restrict__ lam, int B, int M, int nseg,
-                                                         int ntile, const float2 *__restrict__ agg,
+__global__ __launch_bounds__(1024) void k_diag_seg_carry(const float *__restrict__ lam, int conj_lam, int seglen, int B,
+                                                         int M, int nseg, int ntile, const float2 *__restrict__ agg,
                                                          float2 *__restrict__ carry) {
     __shared__ double ga[SEG_NG][64][2];
     const int b = blockIdx.x / ntile, tile = blockIdx.x % ntile;
@@ -554,18 +561,25 @@ __global__ __launch_bounds__(1024) void k_diag_seg_carry(const float *__restrict
     const int m = tile * 64 + ch;
     const bool mok = m < M;
     const int CG = (nseg + SEG_NG - 1) / SEG_NG;
-    const int s0 = grp * CG, s1 = min(s0 + CG, nseg);
+    const int s0 = min(grp * CG, nseg), s1 = min(s0 + CG, nseg);
     cd L = {0.0, 0.0};
-    if (mok) L = cpow(cd{(double)lam[2 * m], (double)lam[2 * m + 1]}, SEG);
+    if (mok) L = cpow(cd{(double)lam[2 * m], conj_lam ? -(double)lam[2 * m + 1] : (double)lam[2 * m + 1]}, seglen);
     const long base = (long)b * nseg;
     double ar = 0.0, ai = 0.0;
     if (mok) {
-        for (int s = s0; s < s1; ++s) {
-            const float2 a = agg[(base + s) * M + m];
-            const double nr = L.re * ar - L.im * ai + (double)a.x;
-            const double ni = L.re * ai + L.im * ar + (double)a.y;
-            ar = nr;
-            ai = ni;
+        for (int s = s0; s < s1; s += SEG_CB) {
+            float2 a[SEG_CB];
+#pragma unroll
+            for (int j = 0; j < SEG_CB; ++j) a[j] = agg[(base + min(s + j, s1 - 1)) * M + m];
+#pragma unroll
+            for (int j = 0; j < SEG_CB; ++j) {
+                if (s + j < s1) {
+                    const double nr = L.re * ar - L.im * ai + (double)a[j].x;
+                    const double ni = L.re * ai + L.im * ar + (double)a[j].y;
+                    ar = nr;
+                    ai = ni;
+                }
+            }
         }
     }
     ga[grp][ch][0] = ar;
@@ -587,13 +601,20 @@ __global__ __launch_bounds__(1024) void k_diag_seg_carry(const float *__restrict
     __syncthreads();
     if (!mok) return;
     double xr = ga[grp][ch][0], xi = ga[grp][ch][1];
-    for (int s = s0; s < s1; ++s) {
-        const float2 a = agg[(base + s) * M + m];
-        carry[(base + s) * M + m] = make_float2((float)xr, (float)xi);
-        const double nr = L.re * xr - L.im * xi + (double)a.x;
-        const double ni = L.re * xi + L.im * xr + (double)a.y;
-        xr = nr;
-        xi = ni;
+    for (int s = s0; s < s1; s += SEG_CB) {
+        float2 a[SEG_CB];
+#pragma unroll
+        for (int j = 0; j < SEG_CB; ++j) a[j] = agg[(base + min(s + j, s1 - 1)) * M + m];
+#pragma unroll
+        for (int j = 0; j < SEG_CB; ++j) {
+            if (s + j < s1) {
+                carry[(base + s + j) * M + m] = make_float2((float)xr, (float)xi);
+                const double nr = L.re * xr - L.im * xi + (double)a[j].x;
+                const double ni = L.re * xi + L.im * xr + (double)a[j].y;
+                xr = nr;
+                xi = ni;
+            }
+        }
     }
 }
 
@@ -633,7 +654,7 @@ static int launch_diag_seg(int B, int T, int M, const float *lam, const float *B
     DEER_LAUNCH_CHECK("k_diag_seg<reduce>");
     {
         KTimer _kt("k_diag_seg_carry", st);
-        hipLaunchKernelGGL(k_diag_seg_carry, dim3(B * ntile), dim3(64 * SEG_NG), 0, st, lam, B, M, nseg, ntile,
+        hipLaunchKernelGGL(k_diag_seg_carry, dim3(B * ntile), dim3(64 * SEG_NG), 0, st, lam, 0, SEG, B, M, nseg, ntile,
                            (const float2 *)agg, carry);
     }
     DEER_LAUNCH_CHECK("k_diag_seg_carry");
@@ -765,19 +786,350 @@ __global__ __launch_bounds__(64) void k_diag_grads_sum2(const double *__restrict
     }
 }
 
+// ---------------------------------------------------------------------------------------
+// Reverse scan of a cotangent g with the parameter gradients, for callers that keep the
+// gradients only (the adjoint itself is not stored): one read of g and of the forward states
+// h, in whole rows (lane = channel, 64 channels per wave).
+//   a_tau = conj(lam) a_{tau+1} + g_tau  (a_T = 0),
+//   dlam_m = sum_{tau >= 1} a_tau conj(h_{tau-1}),   dBc_{m,k} = sum_tau a_tau x_tau[k].
+// Logical positions p = T - 1 - tau; segment r of a sequence covers p in [r S, min(r S + S, T)).
+// A wave walks its segment from a zero state, giving the local adjoint y_p; the adjoint itself
+// is y_p + c_p X_r with c_p = conj(lam)^(p - r S + 1) and X_r the adjoint at p = r S - 1 (the
+// carry).  That is linear in X_r, so the wave accumulates
+//   P1 = sum y conj(h),  P2 = sum c conj(h),  Q1_k = sum y x[k],  Q2_k = sum c x[k]
+// and, once k_diag_seg_carry has formed every X_r from the segment aggregates (y at the
+// segment's last position), k_diag_rseg_sum adds dlam = sum_r P1 + X_r P2 and
+// dBc_k = sum_r Q1_k + X_r Q2_k.  c restarts from a float64 power every RSUB steps; the sums
+// run in float32 per 64 steps and are then added into float32 segment totals.
+// The inputs x of 64 consecutive steps sit one per lane and reach the wave through
+// v_readlane.  Register batches of RSUB steps: the next batch's loads are issued before the
+// current batch is walked.
+// part layout: part[(v B nseg + b nseg + r) M + m], v < 4 + 4 K (P1 re, im, P2 re, im, then
+// per k: Q1 re, im, Q2 re, im); agg[(b nseg + r) M + m].
+// ---------------------------------------------------------------------------------------
+constexpr int RSUB = 8;
+
+template <int K, bool GREAL>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_diag_rseg(const float *__restrict__ lam, const float *__restrict__ g,
+                                                   const float *__restrict__ h, const float *__restrict__ x, int B,
+                                                   int T, int M, int nseg, int S, int ntile,
+                                                   float2 *__restrict__ agg, float *__restrict__ part) {
+    constexpr int NP = 4 + 4 * K;
+    constexpr int GW = GREAL ? 1 : 2;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const long wid = (long)blockIdx.x * 4 + wv;   // (sequence, segment, channel tile)
+    if (wid >= (long)B * nseg * ntile) return;
+    const int tile = (int)(wid % ntile);
+    const long bs = wid / ntile;
+    const int r = (int)(bs % nseg), b = (int)(bs / nseg);
+    const int m = tile * 64 + lane;
+    const bool mok = m < M;
+    const int p0 = r * S, p1 = min(p0 + S, T);
+    float lr = 0.f, li = 0.f;
+    if (mok) {
+        lr = lam[2 * m];
+        li = -lam[2 * m + 1];
+    }
+    const cd lc = {(double)lr, (double)li};
+    const cd lsub = cpow(lc, RSUB);
+    cd cb = lc;   // c at the first step of the current batch
+    // g rows tau and h rows tau - 1 through buffer resources based at row tau_lo of sequence b:
+    // one lane offset for every load (>= 2^31 outside the resource for lanes past M: those loads
+    // return 0) and the row offset in an SGPR
+    const int tau_lo = max(T - p1 - 1, 0);
+    const auto rg = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(g + ((long)b * T + tau_lo) * M * GW),
+                                                      (short)0, 0x7fffffff, 0x00020000);
+    const auto rh = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(h + ((long)b * T + tau_lo) * M * 2),
+                                                      (short)0, 0x7fffffff, 0x00020000);
+    const int vog = mok ? m * 4 * GW : (int)0x80000000, voh = mok ? m * 8 : (int)0x80000000;
+    const float *xb = x + (long)b * (T + 1) * K;
+
+    float gc[RSUB * GW], hc[RSUB * 2], gn[RSUB * GW], hn[RSUB * 2];
+    float xv[K], xn[K];
+    // a batch is guarded when it is partial or holds tau = 0 (no h row before it): then every
+    // load is conditional; other batches load unconditionally
+    auto load_batch = [&](int pb, float *gd, float *hd, auto guard) {
+        constexpr bool GUARD = decltype(guard)::value;
+        const int nv = min(RSUB, p1 - pb);
+#pragma unroll
+        for (int s = 0; s < RSUB; ++s) {
+            const int tau = T - 1 - (pb + s);
+            const int rowo = (tau - tau_lo) * M;
+            float g0 = 0.f, g1 = 0.f, h0 = 0.f, h1 = 0.f;
+            if (!GUARD || s < nv) {
+                if (GREAL) {
+                    g0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rg, vog, rowo * 4, 0));
+                } else {
+                    const v2f t2 = __builtin_bit_cast(v2f, __builtin_amdgcn_raw_buffer_load_b64(rg, vog, rowo * 8, 0));
+                    g0 = t2.x;
+                    g1 = t2.y;
+                }
+                if (!GUARD || tau > 0) {
+                    const v2f t2 =
+                        __builtin_bit_cast(v2f, __builtin_amdgcn_raw_buffer_load_b64(rh, voh, rowo * 8 - M * 8, 0));
+                    h0 = t2.x;
+                    h1 = t2.y;
+                }
+            }
+            gd[s * GW] = g0;
+            if (!GREAL) gd[s * GW + 1] = g1;
+            hd[2 * s] = h0;
+            hd[2 * s + 1] = h1;
+        }
+    };
+    auto guarded = [&](int pb) { return pb + RSUB >= T || pb + RSUB > p1; };
+    auto load_x = [&](int pg, float *xd) {
+        const int p = pg + lane;
+#pragma unroll
+        for (int k = 0; k < K; ++k) xd[k] = p < p1 ? xb[((long)T - 1 - p) * K + k] : 0.f;
+    };
+    float yr = 0.f, yi = 0.f;
+    // segment totals in LDS (each lane its own words, no barrier), float32 sums of 64 steps in
+    // registers
+    __shared__ float tot[4][4 + 4 * K][64];
+    float acc[4 + 4 * K];
+#pragma unroll
+    for (int v = 0; v < NP; ++v) {
+        tot[wv][v][lane] = 0.f;
+        acc[v] = 0.f;
+    }
+    auto walk = [&](int pb, auto guard) {
+        constexpr bool GUARD = decltype(guard)::value;
+        const int q = pb - p0;
+        const int nv = min(RSUB, p1 - pb);
+        float cr = (float)cb.re, ci = (float)cb.im;
+#pragma unroll
+        for (int s = 0; s < RSUB; ++s) {
+            if (!GUARD || s < nv) {
+                const float g0 = gc[s * GW], g1 = GREAL ? 0.f : gc[s * GW + 1];
+                const float nr = fmaf(lr, yr, fmaf(-li, yi, g0));
+                const float ni = fmaf(lr, yi, fmaf(li, yr, g1));
+                yr = nr;
+                yi = ni;
+                const float h0 = hc[2 * s], h1 = hc[2 * s + 1];
+                acc[0] = fmaf(yr, h0, fmaf(yi, h1, acc[0]));
+                acc[1] = fmaf(yi, h0, fmaf(-yr, h1, acc[1]));
+                acc[2] = fmaf(cr, h0, fmaf(ci, h1, acc[2]));
+                acc[3] = fmaf(ci, h0, fmaf(-cr, h1, acc[3]));
+                const int xl = (q & 63) + s;
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    const float xk = lane_bcast(xv[k], xl);
+                    acc[4 + 4 * k] = fmaf(yr, xk, acc[4 + 4 * k]);
+                    acc[5 + 4 * k] = fmaf(yi, xk, acc[5 + 4 * k]);
+                    acc[6 + 4 * k] = fmaf(cr, xk, acc[6 + 4 * k]);
+                    acc[7 + 4 * k] = fmaf(ci, xk, acc[7 + 4 * k]);
+                }
+                const float tr = cr * lr - ci * li;
+                ci = cr * li + ci * lr;
+                cr = tr;
+            }
+        }
+    };
+    using GOFF = std::integral_constant<bool, false>;
+    using GON = std::integral_constant<bool, true>;
+    load_x(p0, xv);
+    if (guarded(p0)) load_batch(p0, gc, hc, GON{});
+    else load_batch(p0, gc, hc, GOFF{});
+    for (int pb = p0; pb < p1; pb += RSUB) {
+        const int q = pb - p0;
+        const bool more = pb + RSUB < p1;
+        const bool newgrp = ((q + RSUB) & 63) == 0;
+        if (more) {
+            if (guarded(pb + RSUB)) load_batch(pb + RSUB, gn, hn, GON{});
+            else load_batch(pb + RSUB, gn, hn, GOFF{});
+            if (newgrp) load_x(pb + RSUB, xn);
+        }
+        if (guarded(pb)) walk(pb, GON{});
+        else walk(pb, GOFF{});
+        cb = cmul(cb, lsub);
+        if (newgrp || !more) {
+#pragma unroll
+            for (int v = 0; v < NP; ++v) {
+                tot[wv][v][lane] += acc[v];
+                acc[v] = 0.f;
+            }
+        }
+        if (more) {
+#pragma unroll
+            for (int e = 0; e < RSUB * GW; ++e) gc[e] = gn[e];
+#pragma unroll
+            for (int e = 0; e < RSUB * 2; ++e) hc[e] = hn[e];
+            if (newgrp) {
+#pragma unroll
+                for (int k = 0; k < K; ++k) xv[k] = xn[k];
+            }
+        }
+    }
+    if (!mok) return;
+    agg[bs * M + m] = make_float2(yr, yi);
+    const long vs = (long)B * nseg * M;
+#pragma unroll
+    for (int v = 0; v < NP; ++v) part[v * vs + bs * M + m] = tot[wv][v][lane];
+}
+
+// float64 sums of the segment terms: dlam = sum_r P1 + X_r P2, dBc_k = sum_r Q1_k + X_r Q2_k.
+// Block = (64-channel tile, slice of the B nseg segment rows), 16 row lanes x 64 channels;
+// a thread loads RSR rows at a time (indices clamped to the slice, loads unconditional) before
+// adding them.  The slice sums go to part2 in the layout k_diag_grads_sum2 reads (value,
+// 16-channel tile, slice, channel).
+constexpr int RSR = 4;
+
+template <int K>
+__global__ __launch_bounds__(1024) void k_diag_rseg_sum(const float2 *__restrict__ carry, const float *__restrict__ part,
+                                                        long rows, int M, int ntile16, double *__restrict__ part2) {
+    constexpr int NV = 2 + 2 * K;
+    constexpr int NP = 4 + 4 * K;
+    __shared__ double red[16][NV][64];
+    const int sl = blockIdx.x % DGS, tile = blockIdx.x / DGS;
+    const int rl = threadIdx.x >> 6, ch = threadIdx.x & 63;
+    const int m = tile * 64 + ch;
+    const bool mok = m < M;
+    const long r0 = rows * sl / DGS, r1 = rows * (sl + 1) / DGS;
+    const long vs = rows * M;
+    double acc[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) acc[v] = 0.0;
+    if (mok && r1 > r0) {
+        for (long rb = r0 + rl; rb < r1; rb += 16 * RSR) {
+            float2 X[RSR];
+            float pv[RSR][NP];
+#pragma unroll
+            for (int j = 0; j < RSR; ++j) {
+                const long row = min(rb + 16 * j, r1 - 1);
+                X[j] = carry[row * M + m];
+#pragma unroll
+                for (int v = 0; v < NP; ++v) pv[j][v] = part[v * vs + row * M + m];
+            }
+#pragma unroll
+            for (int j = 0; j < RSR; ++j) {
+                if (rb + 16 * j < r1) {
+                    const double xr = X[j].x, xi = X[j].y;
+                    double pr = pv[j][2], pi = pv[j][3];
+                    acc[0] += (double)pv[j][0] + (xr * pr - xi * pi);
+                    acc[1] += (double)pv[j][1] + (xr * pi + xi * pr);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        pr = pv[j][6 + 4 * k];
+                        pi = pv[j][7 + 4 * k];
+                        acc[2 + 2 * k] += (double)pv[j][4 + 4 * k] + (xr * pr - xi * pi);
+                        acc[3 + 2 * k] += (double)pv[j][5 + 4 * k] + (xr * pi + xi * pr);
+                    }
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v) red[rl][v][ch] = acc[v];
+    __syncthreads();
+    if (rl < NV && mok) {
+        double t = 0.0;
+#pragma unroll
+        for (int r2 = 0; r2 < 16; ++r2) t += red[r2][rl][ch];
+        part2[(((long)rl * ntile16 + m / 16) * DGS + sl) * 16 + m % 16] = t;
+    }
+}
+
+// segment length of the reverse walk: whole 64-step groups, long enough to keep the carry
+// pass short, short enough for ~4096 waves
+static int diag_rseg_len(int B, int T, int M) {
+    const char *e = getenv("DEER_DIAG_RSEG");
+    if (e && atoi(e) >= 64) return (atoi(e) / 64) * 64;
+    const long ntile = (M + 63) / 64;
+    int S = 1024;
+    while (S > 128 && (long)B * ((T + S - 1) / S) * ntile < 4096) S /= 2;
+    return S;
+}
+
+static bool diag_rseg_enabled() {
+    const char *e = getenv("DEER_DIAG_RSEG");
+    return !e || atoi(e) != 0;
+}
+
+static size_t diag_rseg_ws_bytes(int B, int T, int M, int K) {
+    const int S = diag_rseg_len(B, T, M);
+    const size_t nseg = (T + S - 1) / S;
+    const size_t one = ((size_t)B * nseg * M * sizeof(float2) + 255) & ~(size_t)255;
+    const size_t parts = (((size_t)(4 + 4 * K) * B * nseg * M * sizeof(float)) + 255) & ~(size_t)255;
+    const size_t ntile16 = (M + 15) / 16;
+    const size_t parts2 = (size_t)(2 + 2 * K) * ntile16 * DGS * 16 * sizeof(double);
+    return 2 * one + parts + parts2;
+}
+
 size_t diag_adjoint_ws_bytes(int B, int T, int M, int K) {
     const long ntile = (M + DTC - 1) / DTC;
     const long nq = (T + DCH - 1) / DCH;
     const size_t words = (size_t)B * ntile * nq * DTC * 2 * sizeof(unsigned long long);
     const size_t parts = (size_t)(2 + 2 * K) * B * ntile * nq * DTC * sizeof(float);
     const size_t parts2 = (size_t)(2 + 2 * K) * ntile * DGS * DTC * sizeof(double);
-    return 256 + 2 * ((words + 255) & ~(size_t)255) + ((parts + 255) & ~(size_t)255) + parts2;
+    const size_t lb = 256 + 2 * ((words + 255) & ~(size_t)255) + ((parts + 255) & ~(size_t)255) + parts2;
+    const size_t rs = diag_rseg_ws_bytes(B, T, M, K);
+    return lb > rs ? lb : rs;
 }
 
 // Reverse scan of the cotangent g with the parameter gradients fused (dlam, dBc may be
 // null; lam_out may be null).
 int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const float *g, bool g_real, const float *h,
                         const float *x, float *lam_out, float *dlam, float *dBc, void *ws, hipStream_t st) {
+    const bool grads = dlam || dBc;
+    if (grads && !lam_out && K >= 1 && K <= 4 && diag_rseg_enabled()) {
+        // gradients only: one segment walk over g and h, carries of the segment aggregates,
+        // then the segment terms combined with their carries
+        const int S = diag_rseg_len(B, T, M);
+        const int nseg = (T + S - 1) / S;
+        const int nt64 = (M + 63) / 64, nt16 = (M + 15) / 16;
+        const size_t one = ((size_t)B * nseg * M * sizeof(float2) + 255) & ~(size_t)255;
+        const size_t parts = (((size_t)(4 + 4 * K) * B * nseg * M * sizeof(float)) + 255) & ~(size_t)255;
+        float2 *agg = (float2 *)ws;
+        float2 *carry = (float2 *)((char *)ws + one);
+        float *part = (float *)((char *)ws + 2 * one);
+        double *part2 = (double *)((char *)part + parts);
+        const long waves = (long)B * nseg * nt64;
+        const int grid = (int)((waves + 3) / 4);
+        {
+            KTimer _kt("k_diag_rseg", st);
+#define RSEGK(KV, RE)                                                                                              \
+    hipLaunchKernelGGL((k_diag_rseg<KV, RE>), dim3(grid), dim3(256), 0, st, lam, g, h, x, B, T, M, nseg, S, nt64, agg, \
+                       part)
+#define RSEGALL(RE)                        \
+    switch (K) {                           \
+        case 1: RSEGK(1, RE); break;       \
+        case 2: RSEGK(2, RE); break;       \
+        case 3: RSEGK(3, RE); break;       \
+        default: RSEGK(4, RE); break;      \
+    }
+            if (g_real) {
+                RSEGALL(true)
+            } else {
+                RSEGALL(false)
+            }
+#undef RSEGALL
+#undef RSEGK
+        }
+        DEER_LAUNCH_CHECK("k_diag_rseg");
+        {
+            KTimer _kt("k_diag_seg_carry_rev", st);
+            hipLaunchKernelGGL(k_diag_seg_carry, dim3(B * nt64), dim3(64 * SEG_NG), 0, st, lam, 1, S, B, M, nseg, nt64,
+                               (const float2 *)agg, carry);
+        }
+        DEER_LAUNCH_CHECK("k_diag_seg_carry<rev>");
+        {
+            KTimer _kt("k_diag_grads_sum", st);
+            const long rows = (long)B * nseg;
+            switch (K) {
+                case 1: hipLaunchKernelGGL(k_diag_rseg_sum<1>, dim3(nt64 * DGS), dim3(1024), 0, st, (const float2 *)carry, (const float *)part, rows, M, nt16, part2); break;
+                case 2: hipLaunchKernelGGL(k_diag_rseg_sum<2>, dim3(nt64 * DGS), dim3(1024), 0, st, (const float2 *)carry, (const float *)part, rows, M, nt16, part2); break;
+                case 3: hipLaunchKernelGGL(k_diag_rseg_sum<3>, dim3(nt64 * DGS), dim3(1024), 0, st, (const float2 *)carry, (const float *)part, rows, M, nt16, part2); break;
+                default: hipLaunchKernelGGL(k_diag_rseg_sum<4>, dim3(nt64 * DGS), dim3(1024), 0, st, (const float2 *)carry, (const float *)part, rows, M, nt16, part2); break;
+            }
+            const int nv = 2 + 2 * K;
+            hipLaunchKernelGGL(k_diag_grads_sum2, dim3((nv * nt16 * DTC + 63) / 64), dim3(64), 0, st,
+                               (const double *)part2, K, M, nt16, dlam, dBc);
+        }
+        DEER_LAUNCH_CHECK("k_diag_rseg_sum");
+        return DEER_OK;
+    }
     const int ntile = (M + DTC - 1) / DTC;
     const int nq = (T + DCH - 1) / DCH;
     const int nblk = B * ntile * nq;
@@ -796,7 +1148,6 @@ int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const floa
         hipLaunchKernelGGL(k_zero_u64, dim3(grid), dim3(256), 0, st, (unsigned long long *)ws, n);
     }
     DEER_LAUNCH_CHECK("k_zero_u64");
-    const bool grads = dlam || dBc;
     {
         KTimer _kt(grads ? "k_diag_scan_lb_grads" : "k_diag_scan_lb", st);
 #define LBA(GR, RE, HP, PP)                                                                                        \

@@ -84,6 +84,8 @@ def test_diag_workload_full():
     r = D.deer_readout_loss(ro, h_gpu, c.x, want_masks=True)
     say("deer_adjoint diag full (real g)")
     out = D.deer_adjoint(m, c.x, h_gpu, 0.0, 0, g=r["g"])
+    say("deer_adjoint diag full (real g, gradients only: the step bench.py times)")
+    out_g = D.deer_adjoint(m, c.x, h_gpu, 0.0, 0, g=r["g"], want_lam=False)
     h = O.diag_scan(p["lam"], O.diag_ssm_inputs(p, c.x))
     hg = h_gpu.cpu().numpy()
     assert rel_inf(hg[..., 0] + 1j * hg[..., 1], h) < TOL
@@ -112,5 +114,9 @@ def test_diag_workload_full():
     pg = O.diag_ssm_param_grads(a, h, c.x)
     dl = out["grads"]["lam"].cpu().numpy()
     dB = out["grads"]["Bc"].cpu().numpy()
+    assert rel_inf(dl[..., 0] + 1j * dl[..., 1], pg["lam"]) < TOL
+    assert rel_inf(dB[..., 0] + 1j * dB[..., 1], pg["Bc"]) < TOL
+    dl = out_g["grads"]["lam"].cpu().numpy()
+    dB = out_g["grads"]["Bc"].cpu().numpy()
     assert rel_inf(dl[..., 0] + 1j * dl[..., 1], pg["lam"]) < TOL
     assert rel_inf(dB[..., 0] + 1j * dB[..., 1], pg["Bc"]) < TOL

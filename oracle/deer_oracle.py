@@ -173,6 +173,17 @@ def jacobian_dense(model: dict, mask: np.ndarray) -> np.ndarray:
     return J + np.diag(A)
 
 
+def jacobian_diagonal(model: dict, mask: np.ndarray) -> np.ndarray:
+    """diag(J_F) for masks [..., H], the quasi-DEER approximation of the Jacobian (DEER
+    section, the diagonal replacing J_F in eq. DEER_update): A_i + W_ii m_i (vanilla) or
+    A_i + sum_l W1_il m_l W2_li (shallow)."""
+    A = _p(model, "A")
+    if model["kind"] == "plrnn":
+        return A + np.diagonal(_p(model, "W")) * mask
+    C = _p(model, "W1") * _p(model, "W2").T          # C_il = W1_il W2_li
+    return A + mask @ C.T
+
+
 def forced_jacobians(model: dict, mask: np.ndarray, a: np.ndarray) -> np.ndarray:
     """J~_t = J_F(z~_{t-1}) P_alpha (eq. error_forcing_decomp), dense [B, T, M, M]."""
     return jacobian_dense(model, mask) * (1.0 - a)[None, :]
@@ -249,14 +260,18 @@ def residual_and_masks(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, 
 
 def newton(model: dict, x: np.ndarray, alpha: float, n_forced: int, *, z0=None, init: str = "teacher",
            z_init=None, tol: float = 1e-5, max_iter: int = 500, fixed_iters: int = 0, history: bool = False,
-           gamma: float = 1.0):
+           gamma: float = 1.0, quasi: bool = False):
     """GTF-DEER forward solve.  Each update linearises at z^(k): Delta_t =
     J~_t Delta_{t-1} - r_t, Delta_0 = 0, solved here by the sequential recursion,
     then z^(k+1) = z^(k) + Delta.  Returns dict(z, iters, norms, status[, history]).
 
     gamma scales the linearisation (Delta_t = gamma J~_t Delta_{t-1} - r_t): 1 is Newton's
     step of the algorithm, 0 the fixed-point step z_t <- F(z~_{t-1}); any gamma leaves the
-    fixed point (r = 0) unchanged.  Used to pin the safeguarded GPU iteration."""
+    fixed point (r = 0) unchanged.  Used to pin the safeguarded GPU iteration.
+
+    quasi: quasi-DEER, J~_t replaced by its diagonal diag(J_F(z~_{t-1})) P_alpha (the
+    diagonal approximation discussed with eq. DEER_update), Delta_t = d_t * Delta_{t-1} - r_t;
+    the fixed point is the same."""
     model = _model64(model)
     x = np.asarray(x, f64)
     Bn, T1, _ = x.shape
@@ -289,7 +304,11 @@ def newton(model: dict, x: np.ndarray, alpha: float, n_forced: int, *, z0=None, 
         zt = forced_states(z, zbar, a, z0v)
         r = z - model_map(model, zt)
         mask = activation_mask(model, zt)
-        delta = affine_recurrence(lambda kk, v: gamma * jvp(model, mask[:, kk], p * v), -r)
+        if quasi:
+            dg = jacobian_diagonal(model, mask) * p
+            delta = affine_recurrence(lambda kk, v: gamma * (dg[:, kk] * v), -r)
+        else:
+            delta = affine_recurrence(lambda kk, v: gamma * jvp(model, mask[:, kk], p * v), -r)
         e = np.abs(delta).reshape(Bn, -1).max(axis=1) if T > 0 else np.zeros(Bn)
         e = np.where(np.isnan(delta).reshape(Bn, -1).any(axis=1), np.nan, e)
         upd = active if fixed_iters == 0 else np.ones(Bn, bool)
@@ -350,16 +369,23 @@ def _masks_at(model, x, z, alpha, n_forced, z0, mask_precision):
 
 
 def adjoint(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, *, z0=None,
-            g=None, mask_precision: str = "float64") -> np.ndarray:
+            g=None, mask_precision: str = "float64", quasi: bool = False) -> np.ndarray:
     """lam = dL/dz by the backward recursion lam_T = g_T, lam_{t-1} = J~_t^T lam_t + g_{t-1}
     (eqs. adjoint_eq, backward_recursion with lam = -v).  J~_t is taken at z~_{t-1} of
-    the given trajectory z (normally the converged one)."""
+    the given trajectory z (normally the converged one).
+
+    quasi: the quasi-DEER backward recursion of the gradients appendix, the Jacobians
+    replaced by their diagonals: lam_{t-1} = d_t * lam_t + g_{t-1}, d_t = diag(J~_t).  The
+    parameter gradients then follow from this lam by param_grads unchanged."""
     model = _model64(model)
     z = np.asarray(z, f64)
     M = z.shape[2]
     p = 1.0 - forcing_weights(M, n_forced, alpha)
     mask, _ = _masks_at(model, x, z, alpha, n_forced, z0, mask_precision)
     g = mse_seed(z, x) if g is None else np.asarray(g, f64)
+    if quasi:
+        dg = jacobian_diagonal(model, mask) * p
+        return reverse_affine_recurrence(lambda k, w: dg[:, k] * w, g)
     # J~^T w = P_alpha J_F^T w
     return reverse_affine_recurrence(lambda k, w: p * vjp(model, mask[:, k], w), g)
 

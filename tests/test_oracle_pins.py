@@ -494,3 +494,89 @@ def test_readout_with_given_masks_matches_autograd():
     assert np.allclose(g, hr.grad.numpy(), rtol=1e-10, atol=1e-14)
     for k, v in [("Wa", Wa), ("ca", ca), ("Wb", Wb), ("cb", cb)]:
         assert np.allclose(gr[k], v.grad.numpy(), rtol=1e-10, atol=1e-14), k
+
+
+# ------------------------------------------------------------------------------------
+# quasi-DEER: every forced Jacobian replaced by its diagonal (the diagonal approximation
+# discussed with eq. DEER_update; quasi form of the backward recursion, gradients appendix)
+# ------------------------------------------------------------------------------------
+
+def _diag_blocks(d):
+    """[T, M] diagonals -> [T, M, M] diagonal blocks."""
+    return np.einsum("ti,ij->tij", d, np.eye(d.shape[1]))
+
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+def test_jacobian_diagonal_central_differences(kind):
+    """d_i = dF_i / dz~_i, by central differences of F itself (no ReLU ties nearby)."""
+    M = 5
+    m = _vanilla(M, 41) if kind == "plrnn" else _shallow(M, 9, 42)
+    zt = np.random.default_rng(43).standard_normal((6, M))
+    d = O.jacobian_diagonal(m, O.activation_mask(m, zt))
+    eps = 1e-6
+    for i in range(M):
+        e = np.zeros(M)
+        e[i] = eps
+        fd = (O.model_map(m, zt + e)[:, i] - O.model_map(m, zt - e)[:, i]) / (2 * eps)
+        assert np.allclose(fd, d[:, i], rtol=1e-7, atol=1e-8), i
+
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+def test_quasi_equals_deer_when_every_jacobian_is_diagonal(kind):
+    """Diagonal W (vanilla), or diagonal W1 and W2 with L = M (shallow), make every J_F
+    diagonal: quasi-DEER then takes exactly DEER's steps and has DEER's adjoint."""
+    M, N, T, alpha = 4, 2, 40, 0.25
+    rng = np.random.default_rng(44)
+    A, h = rng.uniform(0.3, 0.8, M), rng.normal(0, 0.1, M)
+    if kind == "plrnn":
+        m = {"kind": "plrnn", "A": A, "W": np.diag(rng.normal(0, 0.5, M)), "h": h}
+    else:
+        m = {"kind": "shplrnn", "A": A, "W1": np.diag(rng.normal(0, 0.7, M)), "W2": np.diag(rng.normal(0, 0.7, M)),
+             "h1": h, "h2": rng.normal(0, 0.1, M)}
+    x = _x(2, T, N, 45)
+    full = O.newton(m, x, alpha, N, fixed_iters=6, history=True)
+    qd = O.newton(m, x, alpha, N, fixed_iters=6, history=True, quasi=True)
+    for a, b in zip(full["history"], qd["history"]):
+        assert np.abs(a - b).max() < 1e-12
+    z = O.rollout(m, x, alpha, N)
+    assert np.allclose(O.adjoint(m, x, z, alpha, N, quasi=True), O.adjoint(m, x, z, alpha, N), rtol=1e-12,
+                       atol=1e-15)
+
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+def test_quasi_update_and_adjoint_are_diagonal_block_solves(kind):
+    """One quasi-DEER update solves the block-bidiagonal system with blocks diag(d_t) below
+    the identity (eq. blockdiag_jacobian with diagonal Jacobians), and the quasi adjoint
+    solves its transpose (LAPACK, dense)."""
+    M, N, T, alpha = 4, 2, 12, 0.3
+    m = _vanilla(M, 46, w_std=0.6) if kind == "plrnn" else _shallow(M, 7, 47)
+    x = _x(1, T, N, 48)
+    p = 1.0 - O.forcing_weights(M, N, alpha)
+    z_init = O.teacher_states(x, M)[:, 1:]
+    res = O.newton(m, x, alpha, N, fixed_iters=1, quasi=True)
+    r, _, mask, _ = O.residual_and_masks(m, x, z_init, alpha, N)
+    D = _diag_blocks(O.jacobian_diagonal(m, mask[0]) * p)
+    assert np.allclose(res["z"][0] - z_init[0], brute.block_bidiagonal_solve(D, -r[0]), rtol=1e-12, atol=1e-14)
+    z = O.rollout(m, x, alpha, N)
+    _, _, mask, _ = O.residual_and_masks(m, x, z, alpha, N)
+    D = _diag_blocks(O.jacobian_diagonal(m, mask[0]) * p)
+    lam = O.adjoint(m, x, z, alpha, N, quasi=True)[0]
+    assert np.allclose(lam, brute.block_bidiagonal_adjoint_solve(D, O.mse_seed(z, x)[0]), rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("kind,M,N,alpha", [("plrnn", 4, 3, 0.2), ("plrnn", 16, 3, 0.2), ("shplrnn", 5, 3, 0.15)])
+def test_quasi_converges_to_rollout_with_prefix_exactness(kind, M, N, alpha):
+    """The quasi step keeps the zero of the residual, so a converged quasi-DEER iterate is the
+    rollout; and with Delta_0 = 0 its first k steps are exact after k updates, like DEER's."""
+    m = _vanilla(M, 49, w_std=0.2) if kind == "plrnn" else _shallow(M, 3 * M, 50)
+    x = _x(2, 50, N, 51)
+    ref = O.rollout(m, x, alpha, N)
+    res = O.newton(m, x, alpha, N, tol=1e-13, max_iter=500, quasi=True)
+    assert res["status"] == "ok"
+    assert np.abs(res["z"] - ref).max() <= 1e-11
+    T = 12
+    xs = x[:, :T + 1]
+    refs = O.rollout(m, xs, alpha, N)
+    hist = O.newton(m, xs, alpha, N, fixed_iters=T, history=True, quasi=True)["history"]
+    for k in range(1, T + 1):
+        assert np.abs(hist[k][:, :k] - refs[:, :k]).max() < 1e-12, k

@@ -18,6 +18,7 @@ second: sum over sequences of T x Newton updates, per second of the whole step.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -43,6 +44,16 @@ def _plrnn_step(D, model, xd, c, ws_s, ws_a):
         raise RuntimeError(f"deer_solve returned status {res['status']}: {D.load().deer_last_error()}")
     # the step's outputs are the parameter gradients: the adjoint itself is not stored
     D.deer_adjoint(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a, want_lam=False)
+    return sum(res["iters"])
+
+
+def _quasi_step(D, model, xd, c, ws_s, ws_a):
+    # quasi-DEER: one more leading step is exact per update, so T + 1 updates always suffice
+    res = D.deer_solve_quasi(model, xd, c.alpha, c.n_obs, tol=c.tol, max_iter=c.T + 2, fixed_iters=c.fixed_iters,
+                             ws=ws_s, check=False)
+    if res["status"] != 0:
+        raise RuntimeError(f"deer_solve_quasi returned status {res['status']}: {D.load().deer_last_error()}")
+    D.deer_adjoint_quasi(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a, want_lam=False)
     return sum(res["iters"])
 
 
@@ -86,6 +97,13 @@ def kernel_work(c, steps, updates):
         out["k_newton_pass16"] = ("mfma", fwd * 2.0 * M ** 3)
         out["k_chunk_product_plrnn"] = ("mfma", steps * B * (T - 1) * 2.0 * M ** 3)
         out["k_resjac_plrnn"] = ("hbm", adj * (4 * M + 4 * N + 4 * W))
+        # quasi-DEER: residual and diagonal (z, x read; r, d written / adjoint: d written),
+        # chunk aggregates (d and r, or d and the seed inputs), fix-ups (forward: d, r, z read
+        # and the next iterate written; reverse: d read, z and x for the forced inputs)
+        out["k_qdeer_resdiag"] = ("hbm", fwd * (12 * M + 4 * N) + adj * (8 * M + 4 * N))
+        out["k_qdeer_chunk"] = ("hbm", fwd * 8 * M + adj * (4 * M + 8 * N))
+        out["k_qdeer_fixup_fwd"] = ("hbm", fwd * 16 * M)
+        out["k_qdeer_fixup_rev"] = ("hbm", adj * (8 * M + 4 * N))
         if M <= 16:
             # the register-tiled fix-ups form the residual and the masks again from z and x:
             # forward z, x read and the next iterate written; reverse z, x read (the training
@@ -267,6 +285,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--quasi", action="store_true",
+                    help="PLRNN workloads: quasi-DEER (diagonal Jacobians) instead of GTF-DEER")
     ap.add_argument("--fig1a", action="store_true",
                     help="instead of the workload: the Fig. 1A sweep, GTF-DEER against the sequential baseline")
     args = ap.parse_args()
@@ -301,9 +321,19 @@ def main():
         step = lambda: _diag_step(D, model, readout, xd, c, ws_s, ws_r, ws_a, bufs)   # noqa: E731
     elif c.kind in ("plrnn", "shplrnn"):
         model = D._Model({"kind": c.kind, **c.params})
-        ws_s = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_SOLVE))
-        ws_a = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_ADJOINT))
-        step = lambda: _plrnn_step(D, model, xd, c, ws_s, ws_a)            # noqa: E731
+        if args.quasi:
+            if c.kind != "plrnn":
+                print("quasi-DEER is built for the vanilla PLRNN workloads (1, 2, 5)", file=sys.stderr)
+                sys.exit(3)
+            lib = D.load()
+            ws_s = D._workspace(lib.deer_quasi_workspace_bytes(ctypes.byref(model.c), c.B, c.T, Bnd.DEER_OP_SOLVE))
+            ws_a = D._workspace(lib.deer_quasi_workspace_bytes(ctypes.byref(model.c), c.B, c.T,
+                                                               Bnd.DEER_OP_ADJOINT))
+            step = lambda: _quasi_step(D, model, xd, c, ws_s, ws_a)        # noqa: E731
+        else:
+            ws_s = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_SOLVE))
+            ws_a = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_ADJOINT))
+            step = lambda: _plrnn_step(D, model, xd, c, ws_s, ws_a)        # noqa: E731
     else:
         print(f"workload {c.name}: model kind {c.kind} not supported by this build", file=sys.stderr)
         sys.exit(3)
@@ -361,11 +391,12 @@ def main():
         "config": {"workload": c.name, "kind": c.kind, "B": c.B, "T": c.T, "M": c.M, "N": c.n_obs,
                    "alpha": c.alpha, "tol": c.tol if not c.fixed_iters else None,
                    "fixed_iters": c.fixed_iters or None, "newton_updates_per_step": iters_per_step,
-                   "step": "deer_solve + deer_adjoint"},
+                   "step": ("deer_solve_quasi + deer_adjoint_quasi (quasi-DEER: diagonal Jacobians)" if args.quasi
+                            else "deer_solve + deer_adjoint")},
         "roofline": roof,
         "kernels": kernels,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.quasi:
         log("[bench] timing the CPU oracle on a bounded sample")
         cb = cpu_baseline(c)
         out["cpu_baseline"] = cb

@@ -21,7 +21,7 @@ from ._binding import DeerError, load  # noqa: F401
 
 __all__ = ["deer_solve", "deer_adjoint", "deer_readout_loss", "plrnn_jacobian", "deer_scan", "deer_workspace_bytes",
            "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_status_string", "DeerError", "load",
-           "deer_sequential", "deer_sequential_workspace_bytes"]
+           "deer_sequential", "deer_sequential_workspace_bytes", "deer_solve_quasi", "deer_adjoint_quasi"]
 
 _KINDS = {"plrnn": _b.DEER_PLRNN, "shplrnn": _b.DEER_SHPLRNN, "diag_ssm": _b.DEER_DIAG_SSM}
 _INITS = {"teacher": _b.DEER_INIT_TEACHER, "zero": _b.DEER_INIT_ZERO, "user": _b.DEER_INIT_USER}
@@ -150,6 +150,23 @@ def deer_solve(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1
     """GTF-DEER forward solve.  Returns dict(z, masks, iters, norms, status).  step_bound:
     threshold of the update safeguard (0: library default, < 0: only non-finite updates are
     rejected)."""
+    return _solve("deer_solve", "deer_workspace_bytes", model, x, alpha, n_forced, z0=z0, tol=tol,
+                  max_iter=max_iter, fixed_iters=fixed_iters, init=init, z=z, want_masks=want_masks, ws=ws,
+                  check=check, step_bound=step_bound)
+
+
+def deer_solve_quasi(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1e-5, max_iter: int = 500,
+                     fixed_iters: int = 0, init: str = "teacher", z=None, want_masks: bool = False, ws=None,
+                     check: bool = True, step_bound: float = 0.0) -> dict:
+    """Quasi-DEER forward solve (diagonal Jacobians; vanilla PLRNN): arguments and result as
+    deer_solve."""
+    return _solve("deer_solve_quasi", "deer_quasi_workspace_bytes", model, x, alpha, n_forced, z0=z0, tol=tol,
+                  max_iter=max_iter, fixed_iters=fixed_iters, init=init, z=z, want_masks=want_masks, ws=ws,
+                  check=check, step_bound=step_bound)
+
+
+def _solve(entry, ws_entry, model, x, alpha, n_forced, *, z0, tol, max_iter, fixed_iters, init, z, want_masks, ws,
+           check, step_bound):
     lib = load()
     m = _model(model)
     x = _dev(x)
@@ -166,17 +183,17 @@ def deer_solve(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1
         H = m.M if m.kind == "plrnn" else m.L
         masks = torch.empty(B, T, (H + 31) // 32, dtype=torch.int32, device="cuda")
     if ws is None:
-        ws = _workspace(lib.deer_workspace_bytes(ctypes.byref(m.c), B, T, _b.DEER_OP_SOLVE))
+        ws = _workspace(getattr(lib, ws_entry)(ctypes.byref(m.c), B, T, _b.DEER_OP_SOLVE))
     iters = (ctypes.c_int32 * B)()
     norms = (ctypes.c_float * B)()
     f = _b.deer_forcing(float(alpha), int(n_forced))
     o = _b.deer_solve_opts(float(tol), int(max_iter), int(fixed_iters), _INITS[init], float(step_bound))
     z0d = _dev(z0)
-    st = lib.deer_solve(ctypes.byref(m.c), ctypes.byref(f), ctypes.byref(o), B, T, _ptr(x), _ptr(z0d), _ptr(out),
-                        _ptr(masks), iters, norms, _ptr(ws), ws.numel(), _stream())
+    st = getattr(lib, entry)(ctypes.byref(m.c), ctypes.byref(f), ctypes.byref(o), B, T, _ptr(x), _ptr(z0d),
+                             _ptr(out), _ptr(masks), iters, norms, _ptr(ws), ws.numel(), _stream())
     if check:
         _check_solve = (_b.DEER_OK, _b.DEER_ERR_NOT_CONVERGED, _b.DEER_ERR_NONFINITE)
-        _b._check(st, "deer_solve", allow=_check_solve)
+        _b._check(st, entry, allow=_check_solve)
     return {"z": out, "masks": masks, "iters": list(iters), "norms": list(norms), "status": st}
 
 
@@ -222,6 +239,31 @@ def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, w
     st = lib.deer_adjoint_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(g),
                              g_layout, _ptr(lam), ctypes.byref(gs), _ptr(ws), ws.numel(), _stream())
     _b._check(st, "deer_adjoint")
+    return {"lam": lam, "grads": grads}
+
+
+def deer_adjoint_quasi(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, want_lam: bool = True,
+                       want_grads: bool = True, ws=None) -> dict:
+    """Quasi-DEER adjoint (diagonal Jacobians; vanilla PLRNN) and parameter gradients at
+    trajectory z: arguments and result as deer_adjoint."""
+    lib = load()
+    m = _model(model)
+    if m.kind != "plrnn":
+        raise ValueError("quasi-DEER is built for the vanilla PLRNN only")
+    x = _dev(x)
+    B, T1, _ = x.shape
+    T = T1 - 1
+    z = _dev(z)
+    g = _dev(g)
+    lam = torch.empty((B, T, m.M), device="cuda") if want_lam else None
+    grads, gs = _plrnn_grads(m) if want_grads else ({}, _b.deer_grads())
+    if ws is None:
+        ws = _workspace(lib.deer_quasi_workspace_bytes(ctypes.byref(m.c), B, T, _b.DEER_OP_ADJOINT))
+    f = _b.deer_forcing(float(alpha), int(n_forced))
+    z0d = _dev(z0)
+    st = lib.deer_adjoint_quasi(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(g),
+                                _ptr(lam), ctypes.byref(gs), _ptr(ws), ws.numel(), _stream())
+    _b._check(st, "deer_adjoint_quasi")
     return {"lam": lam, "grads": grads}
 
 

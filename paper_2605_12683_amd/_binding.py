@@ -23,7 +23,8 @@ DEER_G_NATIVE, DEER_G_REAL = 0, 1
 
 EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "deer_adjoint_ex", "plrnn_jacobian", "deer_scan",
             "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_readout_loss", "deer_status_string",
-            "deer_last_error", "deer_timing_enable", "deer_timing_report"]
+            "deer_last_error", "deer_timing_enable", "deer_timing_report", "deer_solve_quasi", "deer_adjoint_quasi",
+            "deer_quasi_workspace_bytes", "deer_sequential", "deer_sequential_workspace_bytes"]
 
 _fp = ctypes.c_void_p
 
@@ -78,6 +79,12 @@ def load(path: str = LIB_PATH):
     lib.deer_adjoint.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, vp, P(deer_grads), vp, sz,
                                  vp]
     lib.deer_adjoint.restype = i32
+    lib.deer_solve_quasi.argtypes = lib.deer_solve.argtypes
+    lib.deer_solve_quasi.restype = i32
+    lib.deer_adjoint_quasi.argtypes = lib.deer_adjoint.argtypes
+    lib.deer_adjoint_quasi.restype = i32
+    lib.deer_quasi_workspace_bytes.argtypes = [P(deer_model), i32, i32, i32]
+    lib.deer_quasi_workspace_bytes.restype = sz
     lib.deer_adjoint_ex.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, i32, vp, P(deer_grads),
                                     vp, sz, vp]
     lib.deer_adjoint_ex.restype = i32

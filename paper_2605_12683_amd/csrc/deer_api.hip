@@ -349,6 +349,39 @@ static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, 
     return w;
 }
 
+// quasi-DEER workspace: right-hand side and coefficients [B,T,M], chunk aggregates and
+// carries [chains, MP]; solve: the Newton control block and second iterate; adjoint: the
+// per-chain gradient partials and their float64 slices
+struct QuasiWs {
+    float *rhs, *coef, *P, *v, *carry;
+    NewtonCtl ctl;
+    float *gpart;
+    double *gpart2;
+    int C, ncs, MP;
+};
+
+static QuasiWs carve_quasi(void *ws, int B, int T, int M, int op, size_t *bytes) {
+    QuasiWs w{};
+    w.MP = padded_dim(M);
+    w.C = qdeer_chunk_len(B, T, M);
+    w.ncs = (T + w.C - 1) / w.C;
+    const size_t nch = (size_t)B * w.ncs;
+    Carver c(ws);
+    w.coef = c.take<float>((size_t)B * T * M);
+    w.P = c.take<float>(nch * w.MP);
+    w.v = c.take<float>(nch * w.MP);
+    w.carry = c.take<float>(nch * w.MP);
+    if (op == DEER_OP_SOLVE) {
+        w.rhs = c.take<float>((size_t)B * T * M);
+        w.ctl = carve_ctl(c, B, (size_t)T * M, nch);
+    } else {
+        w.gpart = c.take<float>(nch * w.MP * (w.MP + 2));
+        w.gpart2 = c.take<double>(reduce_gpart_ws_bytes(w.MP) / sizeof(double));
+    }
+    *bytes = c.off;
+    return w;
+}
+
 static int check_shallow_limits(const deer_model *m) {
     const size_t cap = 64 * 1024;
     if (sh_resjac_lds(m->M, m->L) > cap || sh_jacform_lds(m->M, m->L) > cap) {
@@ -379,6 +412,16 @@ static int check_common(const deer_model *m, const deer_forcing *f, int B, int T
         return DEER_ERR_INVALID_ARG;
     }
     if ((long)B * (long)T > (1L << 31) / 1) { set_error("B*T too large"); return DEER_ERR_INVALID_ARG; }
+    return DEER_OK;
+}
+
+static int check_quasi(const deer_model *m, const deer_forcing *f, int B, int T) {
+    int rc = check_common(m, f, B, T);
+    if (rc) return rc;
+    if (m->kind != DEER_PLRNN) {
+        set_error("quasi-DEER is built for the vanilla PLRNN (kind DEER_PLRNN) only");
+        return DEER_ERR_INVALID_ARG;
+    }
     return DEER_OK;
 }
 
@@ -704,6 +747,31 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
     return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
 }
 
+static int solve_quasi(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
+                       const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
+                       void *ws, size_t ws_bytes, hipStream_t st) {
+    size_t need = 0;
+    carve_quasi(nullptr, B, T, m->M, DEER_OP_SOLVE, &need);
+    int rc = check_ws(ws, ws_bytes, need);
+    if (rc) return rc;
+    QuasiWs w = carve_quasi(ws, B, T, m->M, DEER_OP_SOLVE, &need);
+    PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
+    if ((rc = init_guess(o, B, T, m->M, f->n_forced, x, z, st))) return rc;
+    std::vector<int> act(B, 1), it(B, 0);
+    std::vector<float> norm(B, NAN);
+    bool nonfinite = false;
+    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *,
+                      uint32_t) -> int {
+        return launch_qdeer_update(a, zb, za, zsel, dact, gam, w.rhs, w.coef, w.P, w.v, w.carry, w.ctl.chain_bits, w.C,
+                                   w.ncs, st);
+    };
+    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ncs, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
+    if (masks) {
+        if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
+    }
+    return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
+}
+
 }  // namespace deer
 
 using namespace deer;
@@ -923,6 +991,47 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
     }
     set_error("deer_adjoint: model kind %d not supported yet", m->kind);
     return DEER_ERR_INVALID_ARG;
+}
+
+int deer_solve_quasi(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
+                     const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
+                     void *ws, size_t ws_bytes, void *stream) {
+    set_error("");
+    int rc = check_quasi(m, f, B, T);
+    if (rc) return rc;
+    if (!o || !x || !z) { set_error("opts, x and z are required"); return DEER_ERR_INVALID_ARG; }
+    if (o->init < 0 || o->init > 2) { set_error("unknown init %d", o->init); return DEER_ERR_INVALID_ARG; }
+    if (!(o->tol >= 0.f) && o->fixed_iters <= 0) { set_error("tol must be >= 0"); return DEER_ERR_INVALID_ARG; }
+    return solve_quasi(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, (hipStream_t)stream);
+}
+
+int deer_adjoint_quasi(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
+                       const float *z, const float *g, float *lam, const deer_grads *grads, void *ws, size_t ws_bytes,
+                       void *stream) {
+    set_error("");
+    int rc = check_quasi(m, f, B, T);
+    if (rc) return rc;
+    if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
+    hipStream_t st = (hipStream_t)stream;
+    size_t need = 0;
+    carve_quasi(nullptr, B, T, m->M, DEER_OP_ADJOINT, &need);
+    if ((rc = check_ws(ws, ws_bytes, need))) return rc;
+    QuasiWs w = carve_quasi(ws, B, T, m->M, DEER_OP_ADJOINT, &need);
+    PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
+    const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
+    if ((rc = launch_qdeer_adjoint(a, g, scale, z, w.coef, w.P, w.v, w.carry, lam, w.gpart, w.C, w.ncs, st))) return rc;
+    if (grads && (grads->A || grads->W || grads->h))
+        return launch_reduce_gpart(w.gpart, B * w.ncs, w.MP, m->M, grads->A, grads->W, grads->h, w.gpart2, st);
+    return DEER_OK;
+}
+
+size_t deer_quasi_workspace_bytes(const deer_model *m, int B, int T, int op) {
+    deer_forcing f{0.f, 0};
+    if (check_quasi(m, &f, B, T) != DEER_OK) return 0;
+    if (op != DEER_OP_SOLVE && op != DEER_OP_ADJOINT) return 0;
+    size_t bytes = 0;
+    carve_quasi(nullptr, B, T, m->M, op, &bytes);
+    return bytes;
 }
 
 static int check_readout(const deer_readout *r, int B, int T, int M) {

@@ -1,0 +1,483 @@
+// Quasi-DEER for the vanilla PLRNN: the GTF-DEER Newton update and backward recursion with
+// every forced Jacobian J~_t replaced by its diagonal (the diagonal approximation the paper
+// discusses with eq. DEER_update, and the quasi form of the backward recursion in the
+// gradients appendix):
+//   forward   Delta_t = d_t * Delta_{t-1} - r_t,        Delta_0 = 0
+//   reverse   lam_{t-1} = d_t * lam_t + g_{t-1},        lam_T = g_T
+//   d_t[i]  = (A_i + W_ii 1[z~_{t-1,i} > 0]) p_i,   p = 1 - a (the forcing projector)
+// Every latent is then an independent first-order recurrence with a coefficient that varies
+// in time, evaluated by a chunked scan: chunk aggregates (prod d, local solution from zero),
+// a float64 carry pass over the chunks of a sequence, and a re-walk of every chunk from its
+// carry.  Array index s holds step s + 1: coef[s] = d_{s+1}, taken at z~_s.
+//
+//   k_qdeer_resdiag   r (forward) and gamma_b d at every (b, s), from the current iterate
+//   k_qdeer_chunk     (prod d, local solution) per (chain, latent)
+//   k_qdeer_carry     carry entering every chunk of a sequence (two levels, float64)
+//   k_qdeer_fixup     forward: z + Delta to the other iterate buffer, per-chain max|Delta| and
+//                     max|z|; reverse: lam (optional) and the gradient partial sums of the
+//                     chain, dW_ij += lam_i relu(z~_j), dA_i += lam_i z~_i, dh_i += lam_i
+//
+// Lanes: a wave holds 64 / MP chains of MP lanes (lane = latent), MP in {16, 32, 64}; the
+// ReLU row of a step goes through LDS when the lanes of a chain need each other's values.
+#include "common.h"
+#include "launch.h"
+
+namespace deer {
+
+namespace {
+__device__ __forceinline__ float q_p(int i, int N, float alpha) { return i < N ? __fsub_rn(1.0f, alpha) : 1.0f; }
+
+// sum_k row[k] * v[k] over the MP values of chain group n in LDS (two partial sums)
+template <int MP>
+__device__ __forceinline__ float q_dot(const float *lds, int n, const float *row) {
+    const float4 *l4 = reinterpret_cast<const float4 *>(lds + n * MP);
+    float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+    for (int q = 0; q < MP / 4; ++q) {
+        const float4 v = l4[q];
+        a0 = fmaf(row[4 * q + 0], v.x, a0);
+        a1 = fmaf(row[4 * q + 1], v.y, a1);
+        a0 = fmaf(row[4 * q + 2], v.z, a0);
+        a1 = fmaf(row[4 * q + 3], v.w, a1);
+    }
+    return a0 + a1;
+}
+
+// coefficient d of step s + 1 from the forced input z~_s, scaled by the damping g
+__device__ __forceinline__ float q_coef(float zt, float Ai, float Wii, float pi, float g) {
+    const float dj = zt > 0.f ? __fadd_rn(Ai, Wii) : Ai;
+    return __fmul_rn(g, __fmul_rn(dj, pi));
+}
+}  // namespace
+
+// ---------------------------------------------------------------------------------------
+// r_s = z_s - F(z~_s) and coef_s = gamma_b d_{s+1} for every (b, s) of the active sequences,
+// at the current iterate of each sequence (zsel).  REV: coef only (the adjoint's right-hand
+// side is the caller's cotangent or the MSE seed, formed in the scan kernels).
+// ---------------------------------------------------------------------------------------
+template <int MP, bool REV>
+__global__ __launch_bounds__(64) void k_qdeer_resdiag(const float *__restrict__ A, const float *__restrict__ W,
+                                                      const float *__restrict__ h, float alpha, int N,
+                                                      const float *__restrict__ x, const float *__restrict__ z0,
+                                                      const float *zbuf, const float *zalt, const int *__restrict__ zsel,
+                                                      const int *__restrict__ active, const float *__restrict__ gamma,
+                                                      float *__restrict__ rhs, float *__restrict__ coef, int B, int T,
+                                                      int M) {
+    constexpr int NCH = 64 / MP;
+    constexpr int NG = 4;   // row groups per pass (memory parallelism)
+    __shared__ __align__(16) float lds[NG][64];
+    const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
+    float wrow[MP];
+#pragma unroll
+    for (int j = 0; j < MP; ++j) wrow[j] = (!REV && i < M && j < M) ? W[i * M + j] : 0.f;
+    const float Ai = i < M ? A[i] : 0.f;
+    const float Wii = i < M ? W[i * M + i] : 0.f;
+    const float hi = (h && i < M) ? h[i] : 0.f;
+    const float pi = q_p(i, N, alpha);
+    const long total = (long)B * T;
+    const long ngroups = (total + NCH - 1) / NCH;
+    for (long grp0 = (long)blockIdx.x * NG; grp0 < ngroups; grp0 += (long)gridDim.x * NG) {
+        float zt[NG], zc[NG], gm[NG];
+        bool act[NG];
+        long rowv[NG];
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            const long row = (grp0 + q) * NCH + n;
+            const bool in = row < total;
+            const int b = in ? (int)(row / T) : 0, s = in ? (int)(row % T) : 0;
+            act[q] = in && i < M && (!active || active[b]);
+            rowv[q] = row;
+            const float *zcur = cur_iter(zbuf, zalt, zsel, b);
+            zt[q] = act[q] ? forced_state(x, z0, zcur, b, s, i, T, M, N, alpha) : 0.f;
+            zc[q] = (act[q] && !REV) ? zcur[(size_t)row * M + i] : 0.f;
+            gm[q] = (gamma && in) ? gamma[b] : 1.f;
+            if (!REV) lds[q][lane] = zt[q] > 0.f ? zt[q] : 0.f;
+        }
+        float F[NG];
+        if (!REV) {
+            lds_barrier();
+#pragma unroll
+            for (int q = 0; q < NG; ++q) {
+                F[q] = fmaf(Ai, zt[q], q_dot<MP>(lds[q], n, wrow)) + hi;
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            lds_barrier();
+        }
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            if (act[q]) {
+                const size_t e = (size_t)rowv[q] * M + i;
+                coef[e] = q_coef(zt[q], Ai, Wii, pi, gm[q]);
+                if (!REV) rhs[e] = zc[q] - F[q];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// Chunk aggregates.  Chain id = b ncs + c covers array indices [s0, s1), s0 = c C.
+//   forward: y_s = coef_s y_{s-1} + sgn rhs_s from y_{s0-1} = 0; P = prod coef_s, v = y_{s1-1}
+//   reverse: y_s = coef_{s+1} y_{s+1} + g_s from y_{s1} = 0 (coef_T = 0);
+//            P = prod coef_{s+1}, v = y_{s0};  g = rhs, or the MSE seed
+//            seed_scale (z_s - x_{s+1}) on the first N latents when rhs is null
+// Loads are issued QB steps at a time (indices clamped to the chain) before they are used.
+// ---------------------------------------------------------------------------------------
+constexpr int QB = 8;
+
+template <int MP, bool REV>
+__global__ __launch_bounds__(64) void k_qdeer_chunk(const float *__restrict__ coef, const float *__restrict__ rhs,
+                                                    float sgn, const float *__restrict__ z, const float *__restrict__ x,
+                                                    float seed_scale, int N, const int *__restrict__ active,
+                                                    float *__restrict__ Pout, float *__restrict__ vout, int B, int T,
+                                                    int M, int C, int ncs) {
+    constexpr int NCH = 64 / MP;
+    const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
+    const int id = blockIdx.x * NCH + n;
+    const bool ok = id < B * ncs && i < M;
+    const int b = ok ? id / ncs : 0, c = ok ? id % ncs : 0;
+    if (!ok || (active && !active[b])) return;
+    const int s0 = c * C, s1 = min(s0 + C, T);
+    const size_t base = (size_t)b * T;
+    float P = 1.f, y = 0.f;
+    for (int k0 = 0; k0 < s1 - s0; k0 += QB) {
+        float cv[QB], gv[QB];
+#pragma unroll
+        for (int k = 0; k < QB; ++k) {
+            const int kk = min(k0 + k, s1 - s0 - 1);
+            const int s = REV ? s1 - 1 - kk : s0 + kk;
+            const int sc = REV ? s + 1 : s;
+            cv[k] = sc < T ? coef[(base + sc) * M + i] : 0.f;
+            if (rhs) {
+                gv[k] = rhs[(base + s) * M + i];
+            } else {
+                gv[k] = i < N ? __fmul_rn(seed_scale, __fsub_rn(z[(base + s) * M + i],
+                                                                 x[((size_t)b * (T + 1) + s + 1) * N + i]))
+                              : 0.f;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < QB; ++k) {
+            if (k0 + k < s1 - s0) {
+                y = fmaf(cv[k], y, sgn * gv[k]);
+                P = P * cv[k];
+            }
+        }
+    }
+    Pout[(size_t)id * MP + i] = P;
+    vout[(size_t)id * MP + i] = y;
+}
+
+// ---------------------------------------------------------------------------------------
+// Carries: block = sequence, threads = (group gq of CG consecutive chunks in processing
+// order, latent i).  X_0 = 0 and X_{l+1} = P_l X_l + v_l over the chunks l in processing
+// order (forward: c = l; reverse: c = ncs - 1 - l); carry[c] = X_l.  Group maps composed in
+// float64, a serial pass over the groups, every group re-walked from its carry.
+// ---------------------------------------------------------------------------------------
+template <int MP, bool REV>
+__global__ __launch_bounds__(1024) void k_qdeer_carry(const float *__restrict__ P, const float *__restrict__ v,
+                                                      float *__restrict__ carry, const int *__restrict__ active, int M,
+                                                      int ncs) {
+    constexpr int NGQ = 1024 / MP;
+    __shared__ double gp[NGQ][MP], gv[NGQ][MP];
+    const int b = blockIdx.x;
+    if (active && !active[b]) return;
+    const int i = threadIdx.x % MP, gq = threadIdx.x / MP;
+    const int CG = (ncs + NGQ - 1) / NGQ;
+    const int l0 = min(gq * CG, ncs), l1 = min(l0 + CG, ncs);
+    const size_t cb = (size_t)b * ncs;
+    auto chunk_of = [&](int l) { return REV ? ncs - 1 - l : l; };
+    double ap = 1.0, av = 0.0;
+    if (i < M) {
+        for (int l = l0; l < l1; l += QB) {
+            float pq[QB], vq[QB];
+#pragma unroll
+            for (int k = 0; k < QB; ++k) {
+                const size_t e = (cb + chunk_of(min(l + k, l1 - 1))) * MP + i;
+                pq[k] = P[e];
+                vq[k] = v[e];
+            }
+#pragma unroll
+            for (int k = 0; k < QB; ++k) {
+                if (l + k < l1) {
+                    av = (double)pq[k] * av + (double)vq[k];
+                    ap = (double)pq[k] * ap;
+                }
+            }
+        }
+    }
+    gp[gq][i] = ap;
+    gv[gq][i] = av;
+    __syncthreads();
+    if (gq == 0 && i < M) {
+        double X = 0.0;
+        for (int g2 = 0; g2 < NGQ; ++g2) {
+            const double xp = gp[g2][i], xv = gv[g2][i];
+            gv[g2][i] = X;
+            X = xp * X + xv;
+        }
+    }
+    __syncthreads();
+    if (i >= M) return;
+    double X = gv[gq][i];
+    for (int l = l0; l < l1; l += QB) {
+        float pq[QB], vq[QB];
+#pragma unroll
+        for (int k = 0; k < QB; ++k) {
+            const size_t e = (cb + chunk_of(min(l + k, l1 - 1))) * MP + i;
+            pq[k] = P[e];
+            vq[k] = v[e];
+        }
+#pragma unroll
+        for (int k = 0; k < QB; ++k) {
+            if (l + k < l1) {
+                carry[(cb + chunk_of(l + k)) * MP + i] = (float)X;
+                X = (double)pq[k] * X + (double)vq[k];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// Forward fix-up: Delta from the carry, the next iterate z + Delta written to the other
+// buffer, per-chain max|Delta| and max|z| bits (reduced per sequence by k_seq_ctl).
+// ---------------------------------------------------------------------------------------
+template <int MP>
+__global__ __launch_bounds__(64) void k_qdeer_fixup_fwd(const float *__restrict__ coef, const float *__restrict__ rhs,
+                                                        const float *__restrict__ carry, float *zbuf, float *zalt,
+                                                        const int *__restrict__ zsel, uint32_t *__restrict__ chain_bits,
+                                                        const int *__restrict__ active, int B, int T, int M, int C,
+                                                        int ncs) {
+    constexpr int NCH = 64 / MP;
+    const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
+    const int id = blockIdx.x * NCH + n;
+    const bool in = id < B * ncs;
+    const int b = in ? id / ncs : 0, c = in ? id % ncs : 0;
+    const bool ok = in && (!active || active[b]);
+    const bool run = ok && i < M;
+    const int s0 = c * C, s1 = ok ? min(s0 + C, T) : s0;
+    const size_t base = (size_t)b * T;
+    const float *zin = cur_iter(zbuf, zalt, zsel, b);
+    float *zout = next_iter(zbuf, zalt, zsel, b);
+    float D = run ? carry[(size_t)id * MP + i] : 0.f;
+    uint32_t emax = 0u, zmax = 0u;
+    for (int k0 = 0; k0 < s1 - s0; k0 += QB) {
+        float cv[QB], rv[QB], zv[QB];
+#pragma unroll
+        for (int k = 0; k < QB; ++k) {
+            const size_t e = (base + s0 + min(k0 + k, s1 - s0 - 1)) * M + i;
+            cv[k] = run ? coef[e] : 0.f;
+            rv[k] = run ? rhs[e] : 0.f;
+            zv[k] = run ? zin[e] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < QB; ++k) {
+            if (run && k0 + k < s1 - s0) {
+                D = fmaf(cv[k], D, -rv[k]);
+                zout[(base + s0 + k0 + k) * M + i] = zv[k] + D;
+                const uint32_t ab = abs_bits(D), zb = abs_bits(zv[k]);
+                emax = emax > ab ? emax : ab;
+                zmax = zmax > zb ? zmax : zb;
+            }
+        }
+    }
+#pragma unroll
+    for (int off = MP / 2; off > 0; off >>= 1) {
+        const uint32_t o = (uint32_t)__shfl_xor((int)emax, off, 64);
+        const uint32_t oz = (uint32_t)__shfl_xor((int)zmax, off, 64);
+        emax = emax > o ? emax : o;
+        zmax = zmax > oz ? zmax : oz;
+    }
+    if (ok && i == 0) {
+        chain_bits[id] = emax;
+        chain_bits[(size_t)B * ncs + id] = zmax;
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// Reverse fix-up: lam from the carry (lam_{s1} of the chunk), walked down the chunk,
+// optionally written, with the gradient partial sums of the chain at the forced inputs
+// z~_s of the same trajectory (the ReLU row of every step through LDS):
+//   gpart[id][i][j] (j < MP) = sum lam_i relu(z~_j),  [MP] = sum lam_i z~_i,  [MP+1] = sum lam_i
+// ---------------------------------------------------------------------------------------
+template <int MP>
+__global__ __launch_bounds__(64) void k_qdeer_fixup_rev(const float *__restrict__ coef, const float *__restrict__ g,
+                                                        float seed_scale, float alpha, int N,
+                                                        const float *__restrict__ x, const float *__restrict__ z0,
+                                                        const float *__restrict__ z, const float *__restrict__ carry,
+                                                        float *__restrict__ lam, float *__restrict__ gpart, int B,
+                                                        int T, int M, int C, int ncs) {
+    constexpr int NCH = 64 / MP;
+    __shared__ __align__(16) float lds[64];
+    const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
+    const int id = blockIdx.x * NCH + n;
+    const bool in = id < B * ncs;
+    const int b = in ? id / ncs : 0, c = in ? id % ncs : 0;
+    const bool run = in && i < M;
+    const int s0 = c * C, s1 = in ? min(s0 + C, T) : s0;
+    // every chain of the wave takes the same number of steps (shorter ones idle), so the
+    // LDS exchange is wave-uniform
+    const int len = s1 - s0;
+    int maxlen = len;
+#pragma unroll
+    for (int off = 32; off >= MP; off >>= 1) maxlen = max(maxlen, __shfl_xor(maxlen, off, 64));
+    const size_t base = (size_t)b * T;
+    float L = run ? carry[(size_t)id * MP + i] : 0.f;
+    float gw[MP], ga = 0.f, gh = 0.f;
+#pragma unroll
+    for (int j = 0; j < MP; ++j) gw[j] = 0.f;
+    for (int k = 0; k < maxlen; ++k) {
+        const bool st = run && k < len;
+        const int s = s1 - 1 - k;
+        float cv = 0.f, gv = 0.f, zt = 0.f;
+        if (st) {
+            cv = s + 1 < T ? coef[(base + s + 1) * M + i] : 0.f;
+            if (g) {
+                gv = g[(base + s) * M + i];
+            } else {
+                gv = i < N ? __fmul_rn(seed_scale, __fsub_rn(z[(base + s) * M + i],
+                                                               x[((size_t)b * (T + 1) + s + 1) * N + i]))
+                           : 0.f;
+            }
+            zt = forced_state(x, z0, z, b, s, i, T, M, N, alpha);
+            L = fmaf(cv, L, gv);
+            if (lam) lam[(base + s) * M + i] = L;
+            ga = fmaf(L, zt, ga);
+            gh += L;
+        }
+        lds[lane] = (st && zt > 0.f) ? zt : 0.f;
+        wave_lds_sync();
+        const float4 *l4 = reinterpret_cast<const float4 *>(lds + n * MP);
+        const float Ls = st ? L : 0.f;
+#pragma unroll
+        for (int q = 0; q < MP / 4; ++q) {
+            const float4 v4 = l4[q];
+            gw[4 * q + 0] = fmaf(Ls, v4.x, gw[4 * q + 0]);
+            gw[4 * q + 1] = fmaf(Ls, v4.y, gw[4 * q + 1]);
+            gw[4 * q + 2] = fmaf(Ls, v4.z, gw[4 * q + 2]);
+            gw[4 * q + 3] = fmaf(Ls, v4.w, gw[4 * q + 3]);
+        }
+        wave_lds_sync();
+    }
+    if (!in) return;
+    float *gp = gpart + ((size_t)id * MP + i) * (MP + 2);
+#pragma unroll
+    for (int j = 0; j < MP; ++j) gp[j] = gw[j];
+    gp[MP] = ga;
+    gp[MP + 1] = gh;
+}
+
+// ---------------------------------------------------------------------------------------
+// host launchers
+// ---------------------------------------------------------------------------------------
+static int q_padded(int M) { return M <= 16 ? 16 : (M <= 32 ? 32 : 64); }
+
+// chunk length: about 4096 waves of chains, at least 16 steps, at most 1024 chunks per
+// sequence (the carry pass walks ncs / (1024 / MP) chunks per thread twice)
+int qdeer_chunk_len(int B, int T, int M) {
+    const int MP = q_padded(M);
+    const long per_wave = 64 / MP;
+    long C = 16;
+    while (C < T && (long)B * ((T + C - 1) / C) > 4096 * per_wave) C *= 2;
+    while ((T + C - 1) / C > 1024) C *= 2;
+    return (int)(C < T ? C : (T > 0 ? T : 1));
+}
+
+static int q_grid_rows(long total, int MP) {
+    const long ngroups = (total + 64 / MP - 1) / (64 / MP);
+    const long want = (ngroups + 3) / 4;
+    return (int)(want < 65536 ? (want > 0 ? want : 1) : 65536);
+}
+
+int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zsel, const int *active,
+                        const float *gamma, float *rhs, float *coef, float *P, float *v, float *carry,
+                        uint32_t *chain_bits, int C, int ncs, hipStream_t st) {
+    const int MP = q_padded(a.M);
+    const int nchains = a.B * ncs;
+    const int gridc = (nchains + 64 / MP - 1) / (64 / MP);
+    {
+        KTimer kt("k_qdeer_resdiag", st);
+        const int grid = q_grid_rows((long)a.B * a.T, MP);
+#define RD(MPV) \
+    hipLaunchKernelGGL((k_qdeer_resdiag<MPV, false>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, \
+                       (const float *)z, (const float *)zalt, zsel, active, gamma, rhs, coef, a.B, a.T, a.M)
+        if (MP == 16) RD(16); else if (MP == 32) RD(32); else RD(64);
+#undef RD
+    }
+    DEER_LAUNCH_CHECK("k_qdeer_resdiag");
+    {
+        KTimer kt("k_qdeer_chunk", st);
+#define CK(MPV) \
+    hipLaunchKernelGGL((k_qdeer_chunk<MPV, false>), dim3(gridc), dim3(64), 0, st, (const float *)coef, (const float *)rhs, \
+                       -1.f, (const float *)nullptr, a.x, 0.f, a.N, active, P, v, a.B, a.T, a.M, C, ncs)
+        if (MP == 16) CK(16); else if (MP == 32) CK(32); else CK(64);
+#undef CK
+    }
+    DEER_LAUNCH_CHECK("k_qdeer_chunk");
+    {
+        KTimer kt("k_qdeer_carry", st);
+#define CR(MPV) \
+    hipLaunchKernelGGL((k_qdeer_carry<MPV, false>), dim3(a.B), dim3(1024), 0, st, (const float *)P, (const float *)v, carry, \
+                       active, a.M, ncs)
+        if (MP == 16) CR(16); else if (MP == 32) CR(32); else CR(64);
+#undef CR
+    }
+    DEER_LAUNCH_CHECK("k_qdeer_carry");
+    {
+        KTimer kt("k_qdeer_fixup_fwd", st);
+#define FX(MPV) \
+    hipLaunchKernelGGL((k_qdeer_fixup_fwd<MPV>), dim3(gridc), dim3(64), 0, st, (const float *)coef, (const float *)rhs, \
+                       (const float *)carry, z, zalt, zsel, chain_bits, active, a.B, a.T, a.M, C, ncs)
+        if (MP == 16) FX(16); else if (MP == 32) FX(32); else FX(64);
+#undef FX
+    }
+    DEER_LAUNCH_CHECK("k_qdeer_fixup_fwd");
+    return DEER_OK;
+}
+
+int launch_qdeer_adjoint(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *coef, float *P,
+                         float *v, float *carry, float *lam, float *gpart, int C, int ncs, hipStream_t st) {
+    const int MP = q_padded(a.M);
+    const int nchains = a.B * ncs;
+    const int gridc = (nchains + 64 / MP - 1) / (64 / MP);
+    {
+        KTimer kt("k_qdeer_resdiag", st);
+        const int grid = q_grid_rows((long)a.B * a.T, MP);
+#define RD(MPV) \
+    hipLaunchKernelGGL((k_qdeer_resdiag<MPV, true>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, z, \
+                       z, (const int *)nullptr, (const int *)nullptr, (const float *)nullptr, (float *)nullptr, coef, \
+                       a.B, a.T, a.M)
+        if (MP == 16) RD(16); else if (MP == 32) RD(32); else RD(64);
+#undef RD
+    }
+    DEER_LAUNCH_CHECK("k_qdeer_resdiag<rev>");
+    {
+        KTimer kt("k_qdeer_chunk", st);
+#define CK(MPV) \
+    hipLaunchKernelGGL((k_qdeer_chunk<MPV, true>), dim3(gridc), dim3(64), 0, st, (const float *)coef, g, 1.f, z, a.x, \
+                       seed_scale, a.N, (const int *)nullptr, P, v, a.B, a.T, a.M, C, ncs)
+        if (MP == 16) CK(16); else if (MP == 32) CK(32); else CK(64);
+#undef CK
+    }
+    DEER_LAUNCH_CHECK("k_qdeer_chunk<rev>");
+    {
+        KTimer kt("k_qdeer_carry", st);
+#define CR(MPV) \
+    hipLaunchKernelGGL((k_qdeer_carry<MPV, true>), dim3(a.B), dim3(1024), 0, st, (const float *)P, (const float *)v, carry, \
+                       (const int *)nullptr, a.M, ncs)
+        if (MP == 16) CR(16); else if (MP == 32) CR(32); else CR(64);
+#undef CR
+    }
+    DEER_LAUNCH_CHECK("k_qdeer_carry<rev>");
+    {
+        KTimer kt("k_qdeer_fixup_rev", st);
+#define FX(MPV) \
+    hipLaunchKernelGGL((k_qdeer_fixup_rev<MPV>), dim3(gridc), dim3(64), 0, st, (const float *)coef, g, seed_scale, a.alpha, \
+                       a.N, a.x, a.z0, z, (const float *)carry, lam, gpart, a.B, a.T, a.M, C, ncs)
+        if (MP == 16) FX(16); else if (MP == 32) FX(32); else FX(64);
+#undef FX
+    }
+    DEER_LAUNCH_CHECK("k_qdeer_fixup_rev");
+    return DEER_OK;
+}
+
+}  // namespace deer

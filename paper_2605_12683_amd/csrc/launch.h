@@ -102,6 +102,17 @@ int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *d
                         double *part2, hipStream_t st);
 size_t reduce_gpart_ws_bytes(int MP);
 
+// quasi-DEER, vanilla PLRNN (diagonal Jacobians): chunk length, one forward Newton update
+// (r and gamma d at the current iterate, chunked diagonal scan, z + Delta to the other buffer,
+// per-chain maxima), and the quasi adjoint with per-chain gradient partials
+// gpart[chain][MP][MP + 2] (MP = padded_dim(M)) for launch_reduce_gpart
+int qdeer_chunk_len(int B, int T, int M);
+int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zsel, const int *active,
+                        const float *gamma, float *rhs, float *coef, float *P, float *v, float *carry,
+                        uint32_t *chain_bits, int C, int ncs, hipStream_t st);
+int launch_qdeer_adjoint(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *coef, float *P,
+                         float *v, float *carry, float *lam, float *gpart, int C, int ncs, hipStream_t st);
+
 // dense stored-Jacobian scan (mode: 0 Newton fix-up, 1 bare forward scan, 2 reverse)
 int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
                                float *P, float *v, const int *active, int C, int ncs, hipStream_t st);

@@ -1,0 +1,88 @@
+"""The C ABI without a GPU: libdeer.so loads, exports every function include/deer.h declares,
+and its host-side logic (workspace sizes, argument validation, status strings) answers
+before any device work is queued."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "deer.h")
+
+_b = pytest.importorskip("paper_2605_12683_amd._binding")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    names = re.findall(r"^\s*(?:const\s+)?(?:int|size_t|char|void|float)\s*\*?\s*(\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_b.LIB_PATH):
+        pytest.skip("libdeer.so is not built (run __graft_entry__.build())")
+    return _b.load()
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ("deer_solve", "deer_adjoint", "plrnn_jacobian", "deer_scan", "deer_solve_quasi", "deer_adjoint_quasi",
+              "deer_workspace_bytes", "deer_status_string", "deer_last_error"):
+        assert n in names, n
+
+
+def test_every_declared_function_is_exported(lib):
+    raw = ctypes.CDLL(_b.LIB_PATH)
+    missing = [n for n in _declared() if not hasattr(raw, n)]
+    assert not missing, missing
+    # the binding declares a signature for every one of them
+    assert set(_b.EXPORTED) <= set(_declared())
+
+
+def _vanilla_model(M=16, kind=_b.DEER_PLRNN):
+    buf = (ctypes.c_float * (M * M))()
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    return _b.deer_model(kind, M, 8 if kind == _b.DEER_SHPLRNN else 0, p, p, p if kind == _b.DEER_SHPLRNN else None,
+                         None, None), buf
+
+
+def test_workspace_queries(lib):
+    m, _keep = _vanilla_model(16)
+    for op in (_b.DEER_OP_SOLVE, _b.DEER_OP_ADJOINT):
+        assert lib.deer_workspace_bytes(ctypes.byref(m), 16, 16384, op) > 0
+        assert lib.deer_quasi_workspace_bytes(ctypes.byref(m), 16, 16384, op) > 0
+    assert lib.deer_workspace_bytes(ctypes.byref(m), 0, 16, _b.DEER_OP_SOLVE) == 0
+    assert lib.deer_workspace_bytes(ctypes.byref(m), 4, 16, 7) == 0
+    bad = _b.deer_model(_b.DEER_PLRNN, 65, 0, m.A, m.W, None, None, None)
+    assert lib.deer_workspace_bytes(ctypes.byref(bad), 4, 16, _b.DEER_OP_SOLVE) == 0
+    sh, _keep2 = _vanilla_model(4, _b.DEER_SHPLRNN)
+    assert lib.deer_quasi_workspace_bytes(ctypes.byref(sh), 4, 16, _b.DEER_OP_SOLVE) == 0   # vanilla only
+
+
+def test_argument_errors_before_device_work(lib):
+    m, _keep = _vanilla_model(4)
+    o = _b.deer_solve_opts(1e-5, 10, 0, 0, 0.0)
+    f = _b.deer_forcing(1.5, 2)                       # alpha outside [0, 1]
+    for entry in ("deer_solve", "deer_solve_quasi"):
+        st = getattr(lib, entry)(ctypes.byref(m), ctypes.byref(f), ctypes.byref(o), 2, 8, None, None, None, None,
+                                 None, None, None, 0, None)
+        assert st == _b.DEER_ERR_INVALID_ARG, entry
+        assert b"alpha" in lib.deer_last_error()
+    f = _b.deer_forcing(0.1, 2)
+    gs = _b.deer_grads()
+    st = lib.deer_adjoint_quasi(ctypes.byref(m), ctypes.byref(f), 2, 8, None, None, None, None, None,
+                                ctypes.byref(gs), None, 0, None)
+    assert st == _b.DEER_ERR_INVALID_ARG                # x and z are required
+    sh, _keep2 = _vanilla_model(4, _b.DEER_SHPLRNN)
+    st = lib.deer_solve_quasi(ctypes.byref(sh), ctypes.byref(f), ctypes.byref(o), 2, 8, None, None, None, None,
+                              None, None, None, 0, None)
+    assert st == _b.DEER_ERR_INVALID_ARG and b"vanilla" in lib.deer_last_error()
+
+
+def test_status_strings(lib):
+    for code in range(6):
+        assert lib.deer_status_string(code)

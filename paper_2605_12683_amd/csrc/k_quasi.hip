@@ -51,9 +51,12 @@ __device__ __forceinline__ float q_coef(float zt, float Ai, float Wii, float pi,
 }  // namespace
 
 // ---------------------------------------------------------------------------------------
-// r_s = z_s - F(z~_s) and coef_s = gamma_b d_{s+1} for every (b, s) of the active sequences,
-// at the current iterate of each sequence (zsel).  REV: coef only (the adjoint's right-hand
-// side is the caller's cotangent or the MSE seed, formed in the scan kernels).
+// r_s = z_s - F(z~_s) and coef_s = gamma_b d_{s+1} for every step s of sequence b =
+// blockIdx.y, at its current iterate (zsel); a converged sequence's blocks exit at once.
+// REV: coef only (the adjoint's right-hand side is the caller's cotangent or the MSE seed,
+// formed in the scan kernels).  A wave takes NG x (64 / MP) consecutive steps per iteration
+// (lane = latent) and loads the next iteration's inputs before it works on the current one.
+// z~ is formed as everywhere else: fl(fl(p z) + fl(alpha x)) on the forced latents.
 // ---------------------------------------------------------------------------------------
 template <int MP, bool REV>
 __global__ __launch_bounds__(64) void k_qdeer_resdiag(const float *__restrict__ A, const float *__restrict__ W,
@@ -64,37 +67,56 @@ __global__ __launch_bounds__(64) void k_qdeer_resdiag(const float *__restrict__ 
                                                       float *__restrict__ rhs, float *__restrict__ coef, int B, int T,
                                                       int M) {
     constexpr int NCH = 64 / MP;
-    constexpr int NG = 4;   // row groups per pass (memory parallelism)
+    constexpr int NG = 4;             // row groups per iteration (memory parallelism)
+    constexpr int RS = NCH * NG;      // steps per iteration
     __shared__ __align__(16) float lds[NG][64];
+    const int b = blockIdx.y;
+    if (active && !active[b]) return;
     const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
+    const bool iok = i < M;
     float wrow[MP];
 #pragma unroll
-    for (int j = 0; j < MP; ++j) wrow[j] = (!REV && i < M && j < M) ? W[i * M + j] : 0.f;
-    const float Ai = i < M ? A[i] : 0.f;
-    const float Wii = i < M ? W[i * M + i] : 0.f;
-    const float hi = (h && i < M) ? h[i] : 0.f;
+    for (int j = 0; j < MP; ++j) wrow[j] = (!REV && iok && j < M) ? W[i * M + j] : 0.f;
+    const float Ai = iok ? A[i] : 0.f;
+    const float Wii = iok ? W[i * M + i] : 0.f;
+    const float hi = (h && iok) ? h[i] : 0.f;
     const float pi = q_p(i, N, alpha);
-    const long total = (long)B * T;
-    const long ngroups = (total + NCH - 1) / NCH;
-    for (long grp0 = (long)blockIdx.x * NG; grp0 < ngroups; grp0 += (long)gridDim.x * NG) {
-        float zt[NG], zc[NG], gm[NG];
-        bool act[NG];
-        long rowv[NG];
+    const float gmb = gamma ? gamma[b] : 1.f;
+    const bool forced = i < N;
+    const float *zs = cur_iter(zbuf, zalt, zsel, b) + (size_t)b * T * M;
+    const float *xs = x + (size_t)b * (T + 1) * N;
+    const float *zst = zs + i;
+    float *cs = coef + (size_t)b * T * M + i;
+    float *rs = REV ? nullptr : rhs + (size_t)b * T * M + i;
+    const float zinit = !iok ? 0.f : (z0 ? z0[(size_t)b * M + i] : (forced ? xs[i] : 0.f));
+    // inputs of the steps of one iteration: z_{s-1}, x_s (forced latents), z_s (residual)
+    float zp[NG], xq[NG], zv[NG];
+    auto load = [&](int sb) {
 #pragma unroll
         for (int q = 0; q < NG; ++q) {
-            const long row = (grp0 + q) * NCH + n;
-            const bool in = row < total;
-            const int b = in ? (int)(row / T) : 0, s = in ? (int)(row % T) : 0;
-            act[q] = in && i < M && (!active || active[b]);
-            rowv[q] = row;
-            const float *zcur = cur_iter(zbuf, zalt, zsel, b);
-            zt[q] = act[q] ? forced_state(x, z0, zcur, b, s, i, T, M, N, alpha) : 0.f;
-            zc[q] = (act[q] && !REV) ? zcur[(size_t)row * M + i] : 0.f;
-            gm[q] = (gamma && in) ? gamma[b] : 1.f;
-            if (!REV) lds[q][lane] = zt[q] > 0.f ? zt[q] : 0.f;
+            const int s = sb + q * NCH + n;
+            const bool ok = s < T && iok;
+            zp[q] = (ok && s > 0) ? zst[(size_t)(s - 1) * M] : 0.f;
+            xq[q] = (ok && s > 0 && forced) ? xs[(size_t)s * N + i] : 0.f;
+            zv[q] = (ok && !REV) ? zst[(size_t)s * M] : 0.f;
         }
+    };
+    const int stride = gridDim.x * RS;
+    int sb = blockIdx.x * RS;
+    load(sb);
+    for (; sb < T; sb += stride) {
+        float zt[NG], zc[NG];
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            const int s = sb + q * NCH + n;
+            zt[q] = s == 0 ? zinit : (forced ? __fadd_rn(__fmul_rn(pi, zp[q]), __fmul_rn(alpha, xq[q])) : zp[q]);
+            zc[q] = zv[q];
+        }
+        load(sb + stride);   // the next iteration's inputs, in flight during this one
         float F[NG];
         if (!REV) {
+#pragma unroll
+            for (int q = 0; q < NG; ++q) lds[q][lane] = zt[q] > 0.f ? zt[q] : 0.f;
             lds_barrier();
 #pragma unroll
             for (int q = 0; q < NG; ++q) {
@@ -105,10 +127,10 @@ __global__ __launch_bounds__(64) void k_qdeer_resdiag(const float *__restrict__ 
         }
 #pragma unroll
         for (int q = 0; q < NG; ++q) {
-            if (act[q]) {
-                const size_t e = (size_t)rowv[q] * M + i;
-                coef[e] = q_coef(zt[q], Ai, Wii, pi, gm[q]);
-                if (!REV) rhs[e] = zc[q] - F[q];
+            const int s = sb + q * NCH + n;
+            if (s < T && iok) {
+                cs[(size_t)s * M] = q_coef(zt[q], Ai, Wii, pi, gmb);
+                if (!REV) rs[(size_t)s * M] = zc[q] - F[q];
             }
         }
     }
@@ -382,10 +404,13 @@ int qdeer_chunk_len(int B, int T, int M) {
     return (int)(C < T ? C : (T > 0 ? T : 1));
 }
 
-static int q_grid_rows(long total, int MP) {
-    const long ngroups = (total + 64 / MP - 1) / (64 / MP);
-    const long want = (ngroups + 3) / 4;
-    return (int)(want < 65536 ? (want > 0 ? want : 1) : 65536);
+// residual grid: y = sequence, x = tiles of 4 (64 / MP) steps, about 4096 blocks in all
+static dim3 q_grid_rows(int B, int T, int MP) {
+    const long tiles = (T + 4L * (64 / MP) - 1) / (4L * (64 / MP));
+    long gx = (4096L + B - 1) / B;
+    if (gx > tiles) gx = tiles;
+    if (gx < 1) gx = 1;
+    return dim3((unsigned)gx, (unsigned)B);
 }
 
 int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zsel, const int *active,
@@ -396,7 +421,7 @@ int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zs
     const int gridc = (nchains + 64 / MP - 1) / (64 / MP);
     {
         KTimer kt("k_qdeer_resdiag", st);
-        const int grid = q_grid_rows((long)a.B * a.T, MP);
+        const dim3 grid = q_grid_rows(a.B, a.T, MP);
 #define RD(MPV) \
     hipLaunchKernelGGL((k_qdeer_resdiag<MPV, false>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, \
                        (const float *)z, (const float *)zalt, zsel, active, gamma, rhs, coef, a.B, a.T, a.M)
@@ -441,7 +466,7 @@ int launch_qdeer_adjoint(const PlrnnArgs &a, const float *g, float seed_scale, c
     const int gridc = (nchains + 64 / MP - 1) / (64 / MP);
     {
         KTimer kt("k_qdeer_resdiag", st);
-        const int grid = q_grid_rows((long)a.B * a.T, MP);
+        const dim3 grid = q_grid_rows(a.B, a.T, MP);
 #define RD(MPV) \
     hipLaunchKernelGGL((k_qdeer_resdiag<MPV, true>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, z, \
                        z, (const int *)nullptr, (const int *)nullptr, (const float *)nullptr, (float *)nullptr, coef, \

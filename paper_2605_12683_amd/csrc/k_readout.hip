@@ -12,7 +12,10 @@
 //   GEMM1  S^T = Wa H^T     A = Wa (LDS), B = H^T (LDS tile of Re h)
 //   GEMM2  G = dS^T Wa      A = dS straight from the GEMM1 accumulator layout (the k index of
 //                           the lane group g is 16n + 4g + r, so no data movement), B = Wa (LDS)
-//   GEMM3  dWa^T += H^T dS^T, accumulated over all tiles of the wave in registers
+//   GEMM3  dWa^T += H^T dS^T, shared by the eight waves of a block: after every round (each
+//          wave one tile) wave w accumulates hidden units 16 w .. 16 w + 15 over the 128 rows
+//          of all eight tiles (dS and H through LDS), so a wave keeps 16 accumulator floats per
+//          lane instead of the whole 128 x 64 dWa, and two waves fit on every SIMD
 // The k ordering of GEMM1 is permuted (k-step (jj, q) uses channel 16 jj + 4 g + q in lane group
 // g) so that four k-steps read one 16-byte LDS vector for both operands.
 #include "common.h"
@@ -24,7 +27,7 @@ namespace {
 constexpr int RH = 128;          // hidden units (padded)
 constexpr int RM = 64;           // state channels (padded)
 constexpr int RNO = 4;           // outputs (padded)
-constexpr int RW = 4;            // waves per block
+constexpr int RW = 8;            // waves per block (one per 16 hidden units in GEMM3)
 constexpr int WS = RM + 4;       // LDS row stride of Wa and of the H tile (16-byte aligned rows)
 constexpr int BS = 17;           // LDS row stride of the [hidden][row] tile
 constexpr int RPS = RH * RM + RNO * RH + RH + RNO + 1;   // partial floats per wave
@@ -43,6 +46,7 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
     __shared__ __align__(16) float hti[RW][16][WS];
     __shared__ float buf[GRADS ? RW : 1][RH][BS];
     __shared__ float dyv[GRADS ? RW : 1][16][RNO];
+    __shared__ float lsw[RW];
     const int M = ra.M, H = ra.H, No = ra.No;
     const int tid = threadIdx.x;
     for (int e = tid; e < RH * RM; e += RW * 64) {
@@ -63,27 +67,33 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
     const long ntiles = (rows + 15) / 16;
     const int HW = (H + 31) / 32;
 
-    v4f acc3[4][8];                 // dWa^T tiles [channel tile q][hidden tile n]
+    v4f acc3[4];                    // dWa^T tiles [channel tile q] of hidden tile n = wv
     float dwb[RNO][2], dca[2], dcb[RNO], lsum = 0.f;
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int n = 0; n < 8; ++n) acc3[q][n] = (v4f){0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < 4; ++q) acc3[q] = (v4f){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int o = 0; o < RNO; ++o) dwb[o][0] = dwb[o][1] = dcb[o] = 0.f;
     dca[0] = dca[1] = 0.f;
 
     // Re h of a tile (one 512-byte row segment per load at M = 64), loaded one tile ahead
     float hv[16];
+    // through a buffer resource that ends at the last row: rows past the end, and lanes past M
+    // (lane offset >= 2^31), load 0 without branches (the whole offset is in the VGPR, so the
+    // range check covers it)
+    const int voh = lane < M ? lane * 8 : (int)0x80000000;
     auto load_tile = [&](long tl) {
-        const long rb = tl * 16;
+        const long rb = tl < ntiles ? tl * 16 : rows;
+        const long left = rows - rb;
+        const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(h + rb * M * 2), (short)0,
+                                                          (int)(left < 16 ? left * M * 8 : 16L * M * 8), 0x00020000);
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-            hv[i] = (tl < ntiles && rb + i < rows && lane < M) ? h[((rb + i) * M + lane) * 2] : 0.f;
+        for (int i = 0; i < 16; ++i) hv[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, voh + i * M * 8, 0, 0));
     };
-    long tile = (long)blockIdx.x * RW + wv;
-    load_tile(tile);
-    for (; tile < ntiles; tile += (long)gridDim.x * RW) {
+    // rounds are block-uniform (GEMM3 needs every wave at its barriers); a wave whose tile
+    // lies past the end works on zero rows, which contribute nothing
+    load_tile((long)blockIdx.x * RW + wv);
+    for (long base = (long)blockIdx.x * RW; base < ntiles; base += (long)gridDim.x * RW) {
+        const long tile = base + wv;
         const long r0 = tile * 16;
 #pragma unroll
         for (int i = 0; i < 16; ++i) hti[wv][i][lane] = hv[i];
@@ -155,8 +165,16 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
         }
         float dy[RNO];
         {
-            const long bq = rok ? row / T : 0, tq = rok ? row % T : 0;
-            const float *xt = x + (bq * (T + 1) + tq + 1) * No;
+            // target row t + 1 of sequence b for row = b T + t: x row index row + b + 1, with
+            // b from the tile's first row (one scalar division) and the sequence boundaries
+            // inside the tile
+            // inside the tile (rows past the end read row 1 of a valid sequence, unused)
+            const uint32_t Tu = (uint32_t)T;
+            const uint32_t b0 = __builtin_amdgcn_readfirstlane((uint32_t)(r0 < rows ? r0 : 0) / Tu);
+            const uint32_t rowu = rok ? (uint32_t)row : b0 * Tu;
+            uint32_t bq = b0;
+            for (int k = 0; k < 16 && rowu >= (bq + 1) * Tu; ++k) ++bq;
+            const float *xt = x + ((size_t)rowu + bq + 1) * No;
 #pragma unroll
             for (int o = 0; o < RNO; ++o) {
                 const bool ok = rok && o < No;
@@ -220,50 +238,56 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
 #pragma unroll
                 for (int q = 0; q < 4; ++q) acc2[q] = mfma16x16x4(acc1[n][r], wa[hid][16 * q + c], acc2[q]);
             }
+        {
+            // g rows r0 + 4 g + r, channels 16 q + c: stores through a resource that ends at the
+            // last row (later rows dropped; the whole offset in the VGPR, so the range check
+            // covers it), lanes past M get an offset outside it
+            const long left = rows - r0 < 0 ? 0 : (rows - r0 < 16 ? rows - r0 : 16);
+            const auto rs = __builtin_amdgcn_make_buffer_rsrc(gout + (r0 < rows ? r0 : 0) * M, (short)0,
+                                                              (int)(left * M * 4), 0x00020000);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int ch = 16 * q + c;
+            for (int q = 0; q < 4; ++q) {
+                const int ch = 16 * q + c;
+                const int vo = ch < M ? (4 * g * M + ch) * 4 : (int)0x80000000;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const long rw = r0 + 4 * g + r;
-                if (rw < rows && ch < M) gout[rw * M + ch] = acc2[q][r];
+                for (int r = 0; r < 4; ++r)
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc2[q][r]), rs, vo + r * M * 4, 0, 0);
             }
         }
         if (GRADS) {
-            // ds to LDS [hidden][row]; dca; GEMM3
+            // ds to LDS [hidden][row]; dca; GEMM3 over the block's eight tiles
 #pragma unroll
             for (int n = 0; n < 8; ++n)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) buf[wv][16 * n + 4 * g + r][c] = acc1[n][r];
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            lds_barrier();
 #pragma unroll
             for (int rr = 0; rr < 16; ++rr) {
                 dca[0] += buf[wv][2 * lane][rr];
                 dca[1] += buf[wv][2 * lane + 1][rr];
             }
+#pragma unroll 2
+            for (int w2 = 0; w2 < RW; ++w2) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                float bv[8];
+                for (int j = 0; j < 4; ++j) {
+                    const float bv = buf[w2][16 * wv + c][4 * j + g];
 #pragma unroll
-                for (int n = 0; n < 8; ++n) bv[n] = buf[wv][16 * n + c][4 * j + g];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const float av = hti[wv][4 * j + g][16 * q + c];
-#pragma unroll
-                    for (int n = 0; n < 8; ++n) acc3[q][n] = mfma16x16x4(av, bv[n], acc3[q][n]);
+                    for (int q = 0; q < 4; ++q) acc3[q] = mfma16x16x4(hti[w2][4 * j + g][16 * q + c], bv, acc3[q]);
                 }
             }
+            // the next round overwrites hti and buf: every wave is past its reads
+            lds_barrier();
+        } else {
+            // the next tile overwrites hti: every lane is past its reads
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         }
-        // the next tile overwrites hti and buf: every lane is past its reads
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
 
-    // per-wave partials: [dWa (RH x RM) | dWb (RNO x RH) | dca (RH) | dcb (RNO) | sum err^2]
-    float *pw = part + ((long)blockIdx.x * RW + wv) * RPS_PAD;
+    // per-block partials: [dWa (RH x RM) | dWb (RNO x RH) | dca (RH) | dcb (RNO) | sum err^2];
+    // every wave writes its hidden rows of dWa, the rest is summed over the block's waves
+    float *pb = part + (long)blockIdx.x * RPS_PAD;
 #pragma unroll
     for (int o = 0; o < RNO; ++o) {
 #pragma unroll
@@ -271,32 +295,50 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
     }
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) lsum += __shfl_xor(lsum, off, 64);
+    constexpr int RV = RNO * RH + RH + RNO + 1;
     if (GRADS) {
+        static_assert(RW * RV <= RW * RH * BS, "block sums fit in the dS tiles");
+        float *red = &buf[0][0][0];
+        float *rw = red + wv * RV;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
 #pragma unroll
-            for (int n = 0; n < 8; ++n)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) pw[(16 * n + c) * RM + 16 * q + 4 * g + r] = acc3[q][n][r];
+            for (int r = 0; r < 4; ++r) pb[(16 * wv + c) * RM + 16 * q + 4 * g + r] = acc3[q][r];
 #pragma unroll
         for (int o = 0; o < RNO; ++o) {
-            pw[RH * RM + o * RH + 2 * lane] = dwb[o][0];
-            pw[RH * RM + o * RH + 2 * lane + 1] = dwb[o][1];
+            rw[o * RH + 2 * lane] = dwb[o][0];
+            rw[o * RH + 2 * lane + 1] = dwb[o][1];
         }
-        pw[RH * RM + RNO * RH + 2 * lane] = dca[0];
-        pw[RH * RM + RNO * RH + 2 * lane + 1] = dca[1];
+        rw[RNO * RH + 2 * lane] = dca[0];
+        rw[RNO * RH + 2 * lane + 1] = dca[1];
         if (lane < RNO) {
             float v = dcb[0];
 #pragma unroll
             for (int o = 1; o < RNO; ++o)
                 if (lane == o) v = dcb[o];
-            pw[RH * RM + RNO * RH + RH + lane] = v;
+            rw[RNO * RH + RH + lane] = v;
+        }
+        if (lane == 0) rw[RV - 1] = lsum;
+        __syncthreads();
+        for (int e = tid; e < RV; e += RW * 64) {
+            float t = 0.f;
+#pragma unroll
+            for (int w2 = 0; w2 < RW; ++w2) t += red[w2 * RV + e];
+            pb[RH * RM + e] = t;
+        }
+    } else {
+        if (lane == 0) lsw[wv] = lsum;
+        __syncthreads();
+        if (tid == 0) {
+            float t = 0.f;
+#pragma unroll
+            for (int w2 = 0; w2 < RW; ++w2) t += lsw[w2];
+            pb[RPS - 1] = t;
         }
     }
-    if (lane == 0) pw[RPS - 1] = lsum;
 }
 
-// float64 sums of the per-wave partials: stage 1 over slices of the waves, stage 2 over slices
+// float64 sums of the per-block partials: stage 1 over slices of the blocks, stage 2 over slices
 constexpr int RO_SLICES = 256;
 
 __global__ __launch_bounds__(256) void k_readout_sum1(const float *__restrict__ part, int nwaves, int only_loss,
@@ -359,14 +401,14 @@ static int readout_grid(long rows) {
 
 size_t readout_ws_bytes(int B, int T) {
     const int grid = readout_grid((long)B * T);
-    const size_t p1 = ((size_t)grid * RW * RPS_PAD * sizeof(float) + 255) & ~(size_t)255;
+    const size_t p1 = ((size_t)grid * RPS_PAD * sizeof(float) + 255) & ~(size_t)255;
     return p1 + (size_t)RO_SLICES * RPS * sizeof(double);
 }
 
 int launch_readout(const RoArgs &ra, int B, int T, const float *h, const float *x, float *g, uint32_t *masks,
                    float *loss, const RoGrads &gr, void *ws, hipStream_t st) {
     const int grid = readout_grid((long)B * T);
-    const size_t p1 = ((size_t)grid * RW * RPS_PAD * sizeof(float) + 255) & ~(size_t)255;
+    const size_t p1 = ((size_t)grid * RPS_PAD * sizeof(float) + 255) & ~(size_t)255;
     float *part = (float *)ws;
     double *part2 = (double *)((char *)ws + p1);
     const float scale = 2.0f / ((float)B * (float)ra.No * (float)T);
@@ -382,7 +424,7 @@ int launch_readout(const RoArgs &ra, int B, int T, const float *h, const float *
     DEER_LAUNCH_CHECK("k_readout");
     if (grads || loss) {
         KTimer _kt("k_readout_sum", st);
-        hipLaunchKernelGGL(k_readout_sum1, dim3(RO_SLICES), dim3(256), 0, st, (const float *)part, grid * RW,
+        hipLaunchKernelGGL(k_readout_sum1, dim3(RO_SLICES), dim3(256), 0, st, (const float *)part, grid,
                            grads ? 0 : 1, part2);
         hipLaunchKernelGGL(k_readout_sum2, dim3((RPS + 255) / 256), dim3(256), 0, st, (const double *)part2, gr, ra.M,
                            ra.H, ra.No, 0.5f * scale, loss);

@@ -188,6 +188,12 @@ static int group_maps_override() {
     return e ? atoi(e) : -1;
 }
 
+// DEER_SMALL=0 keeps small fixed-update solves on the general path (a test override)
+static bool small_path_enabled() {
+    const char *e = getenv("DEER_SMALL");
+    return !e || atoi(e) != 0;
+}
+
 // DEER_PASS_FUSION=0 keeps the M <= 16 fix-up and forward pass in separate kernels where the
 // fused pass kernel would apply (a test override)
 static bool pass_fusion_allowed() {
@@ -670,6 +676,20 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     std::vector<int> act(B, 1), it(B, 0);
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
+    if (small_path_enabled() && newton_small_fits(m->M, T, o->fixed_iters)) {
+        // every update in one launch; the last update's norms read once
+        if ((rc = launch_newton_small(a, z, o->fixed_iters, w.ctl.norm_bits, st))) return rc;
+        std::vector<uint32_t> nb(B, 0);
+        DEER_HIP(hipMemcpyAsync(nb.data(), w.ctl.norm_bits, B * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+        DEER_HIP(hipStreamSynchronize(st));
+        for (int b = 0; b < B; ++b) {
+            memcpy(&norm[b], &nb[b], 4);
+            it[b] = o->fixed_iters;
+            if (!isfinite(norm[b])) nonfinite = true;
+        }
+        if (masks && (rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
+        return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
+    }
     // M <= 16: the fix-up also takes the pass-end control of the adaptive loop
     NewtonCtl ctl = w.ctl;
     ctl.fused = w.MP == 16 && o->fixed_iters <= 0;

@@ -102,6 +102,12 @@ int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *d
                         double *part2, hipStream_t st);
 size_t reduce_gpart_ws_bytes(int MP);
 
+// small vanilla PLRNNs (M <= 4, T <= 4096) with a fixed number of plain Newton updates: the
+// whole solve in one launch (one workgroup per sequence, update in place); norm_bits[b] gets
+// max |Delta| of the last update
+bool newton_small_fits(int M, int T, int fixed_iters);
+int launch_newton_small(const PlrnnArgs &a, float *z, int iters, uint32_t *norm_bits, hipStream_t st);
+
 // quasi-DEER, vanilla PLRNN (diagonal Jacobians): chunk length, one forward Newton update
 // (r and gamma d at the current iterate, chunked diagonal scan, z + Delta to the other buffer,
 // per-chain maxima), and the quasi adjoint with per-chain gradient partials

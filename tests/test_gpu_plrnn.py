@@ -69,6 +69,34 @@ def test_config1_fixed_five_iterations():
     assert res["iters"] == [5]
 
 
+@pytest.mark.parametrize("M,N,B,T,k", [(1, 1, 1, 1, 1), (2, 1, 3, 17, 3), (3, 3, 1, 1024, 5), (4, 4, 2, 4096, 4),
+                                     (3, 2, 2, 300, 7), (4, 2, 1, 255, 2)])
+@pytest.mark.parametrize("user_z0", [False, True])
+def test_small_solve_in_one_launch(M, N, B, T, k, user_z0):
+    """Small models with a fixed number of updates run the whole solve in one workgroup per
+    sequence (chunk maps, two-level carries, in-place fix-up): the oracle's k-th Newton iterate,
+    and the general path's (DEER_SMALL=0), with the masks at the result."""
+    c = _case(M, N, B, T, 0.2, 200 + M + T)
+    m = oracle_model(c)
+    z0 = np.random.default_rng(M).standard_normal((B, M)).astype(np.float32) if user_z0 else None
+    say("deer_solve small one-launch", M, N, B, T, k, user_z0)
+    res = D.deer_solve(m, c.x, c.alpha, N, fixed_iters=k, z0=z0, want_masks=True)
+    ref = O.newton(m, c.x, c.alpha, N, fixed_iters=k, z0=z0)
+    assert res["status"] == 0 and res["iters"] == [k] * B
+    z = res["z"].cpu().numpy()
+    assert rel_inf(z, ref["z"]) < TOL
+    assert np.all(np.abs(np.asarray(res["norms"]) - ref["norms"]) <= 1e-4 * (1.0 + np.abs(ref["norms"])))
+    fp32 = O.activation_mask_fp32(m, z, c.x, c.alpha, N, z0)
+    assert np.array_equal(masks_to_bool(res["masks"].cpu().numpy(), M), fp32)
+    os.environ["DEER_SMALL"] = "0"
+    try:
+        say("deer_solve general path", M, N, B, T, k, user_z0)
+        gen = D.deer_solve(m, c.x, c.alpha, N, fixed_iters=k, z0=z0)
+    finally:
+        os.environ.pop("DEER_SMALL", None)
+    assert rel_inf(z, gen["z"].cpu().numpy()) < TOL
+
+
 @pytest.mark.parametrize("M,N,B,T,alpha,chunk", [
     (3, 3, 1, 300, 0.1, 0), (3, 3, 2, 300, 0.1, 17), (16, 3, 3, 1000, 0.2, 0), (16, 3, 2, 777, 0.2, 64),
     (20, 4, 2, 513, 0.3, 100), (32, 32, 2, 600, 0.1, 0), (40, 10, 2, 300, 0.3, 33), (64, 64, 2, 400, 0.05, 0),

@@ -164,9 +164,11 @@ int deer_adjoint(const deer_model *model, const deer_forcing *forcing, int B, in
                  const float *x, const float *z0, const float *z, const float *g,
                  float *lam, const deer_grads *grads, void *ws, size_t ws_bytes, void *stream);
 
-/* Quasi-DEER (vanilla PLRNN only): deer_solve and deer_adjoint with every forced Jacobian
+/* Quasi-DEER (PLRNN kinds): deer_solve and deer_adjoint with every forced Jacobian
  * J~_t replaced by its diagonal d_t = diag(J_F(z~_{t-1})) P_alpha, i.e.
- * d_t[i] = (A_i + W_ii 1[z~_{t-1,i} > 0]) (1 - a_i) -- the quasi-Newton variant the paper sets
+ * d_t[i] = (A_i + W_ii 1[z~_{t-1,i} > 0]) (1 - a_i) for the vanilla PLRNN and
+ * d_t[i] = (A_i + sum_l W_il 1[u_l > 0] W2_li) (1 - a_i), u = W2 z~_{t-1} + h2, for the shallow
+ * one (same limits as deer_solve) -- the quasi-Newton variant the paper sets
  * against full Jacobians (section on DEER, the diagonal approximation of eq. DEER_update;
  * quasi form of the backward recursion in the gradients appendix; ablation of Jacobian
  * diagonalisation).  Updates: Delta_t = d_t Delta_{t-1} - r_t (the same zero of the residual,
@@ -175,7 +177,7 @@ int deer_adjoint(const deer_model *model, const deer_forcing *forcing, int B, in
  * as in deer_adjoint (an approximation of the true gradient that ignores the mixing between
  * latents).  Arguments, outputs, the safeguard and the status codes are those of
  * deer_solve / deer_adjoint; the workspace is deer_quasi_workspace_bytes(model, B, T, op)
- * bytes.  Kinds other than DEER_PLRNN return DEER_ERR_INVALID_ARG. */
+ * bytes.  DEER_DIAG_SSM returns DEER_ERR_INVALID_ARG (its recurrence is already diagonal). */
 int deer_solve_quasi(const deer_model *model, const deer_forcing *forcing, const deer_solve_opts *opts,
                      int B, int T, const float *x, const float *z0, float *z, uint32_t *masks,
                      int32_t *iters, float *final_norm, void *ws, size_t ws_bytes, void *stream);

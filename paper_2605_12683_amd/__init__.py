@@ -158,7 +158,7 @@ def deer_solve(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1
 def deer_solve_quasi(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1e-5, max_iter: int = 500,
                      fixed_iters: int = 0, init: str = "teacher", z=None, want_masks: bool = False, ws=None,
                      check: bool = True, step_bound: float = 0.0) -> dict:
-    """Quasi-DEER forward solve (diagonal Jacobians; vanilla PLRNN): arguments and result as
+    """Quasi-DEER forward solve (diagonal Jacobians; PLRNN kinds): arguments and result as
     deer_solve."""
     return _solve("deer_solve_quasi", "deer_quasi_workspace_bytes", model, x, alpha, n_forced, z0=z0, tol=tol,
                   max_iter=max_iter, fixed_iters=fixed_iters, init=init, z=z, want_masks=want_masks, ws=ws,
@@ -244,12 +244,12 @@ def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, w
 
 def deer_adjoint_quasi(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, want_lam: bool = True,
                        want_grads: bool = True, ws=None) -> dict:
-    """Quasi-DEER adjoint (diagonal Jacobians; vanilla PLRNN) and parameter gradients at
+    """Quasi-DEER adjoint (diagonal Jacobians; PLRNN kinds) and parameter gradients at
     trajectory z: arguments and result as deer_adjoint."""
     lib = load()
     m = _model(model)
-    if m.kind != "plrnn":
-        raise ValueError("quasi-DEER is built for the vanilla PLRNN only")
+    if m.kind not in ("plrnn", "shplrnn"):
+        raise ValueError("quasi-DEER is built for the PLRNN kinds")
     x = _dev(x)
     B, T1, _ = x.shape
     T = T1 - 1

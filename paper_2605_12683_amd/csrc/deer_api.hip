@@ -358,15 +358,19 @@ static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, 
 // quasi-DEER workspace: right-hand side and coefficients [B,T,M], chunk aggregates and
 // carries [chains, MP]; solve: the Newton control block and second iterate; adjoint: the
 // per-chain gradient partials and their float64 slices
+// (shallow PLRNN, L > 0: the hidden-unit masks; adjoint: the adjoint itself when the caller
+// does not keep it, and the partial sums of the shallow gradient kernel)
 struct QuasiWs {
     float *rhs, *coef, *P, *v, *carry;
     NewtonCtl ctl;
     float *gpart;
     double *gpart2;
+    uint32_t *masks;
+    float *lam, *part;
     int C, ncs, MP;
 };
 
-static QuasiWs carve_quasi(void *ws, int B, int T, int M, int op, size_t *bytes) {
+static QuasiWs carve_quasi(void *ws, int B, int T, int M, int L, int op, size_t *bytes) {
     QuasiWs w{};
     w.MP = padded_dim(M);
     w.C = qdeer_chunk_len(B, T, M);
@@ -377,9 +381,14 @@ static QuasiWs carve_quasi(void *ws, int B, int T, int M, int op, size_t *bytes)
     w.P = c.take<float>(nch * w.MP);
     w.v = c.take<float>(nch * w.MP);
     w.carry = c.take<float>(nch * w.MP);
+    if (L > 0) w.masks = c.take<uint32_t>((size_t)B * T * ((L + 31) / 32));
     if (op == DEER_OP_SOLVE) {
         w.rhs = c.take<float>((size_t)B * T * M);
         w.ctl = carve_ctl(c, B, (size_t)T * M, nch);
+    } else if (L > 0) {
+        w.lam = c.take<float>((size_t)B * T * M);
+        int nb = 0;
+        w.part = c.take<float>(sh_grads_part_floats(M, L, &nb));
     } else {
         w.gpart = c.take<float>(nch * w.MP * (w.MP + 2));
         w.gpart2 = c.take<double>(reduce_gpart_ws_bytes(w.MP) / sizeof(double));
@@ -387,6 +396,8 @@ static QuasiWs carve_quasi(void *ws, int B, int T, int M, int op, size_t *bytes)
     *bytes = c.off;
     return w;
 }
+
+static int quasi_L(const deer_model *m) { return m->kind == DEER_SHPLRNN ? m->L : 0; }
 
 static int check_shallow_limits(const deer_model *m) {
     const size_t cap = 64 * 1024;
@@ -397,6 +408,8 @@ static int check_shallow_limits(const deer_model *m) {
     }
     return DEER_OK;
 }
+
+
 
 static int check_common(const deer_model *m, const deer_forcing *f, int B, int T) {
     if (!m || !f) { set_error("model/forcing pointer is NULL"); return DEER_ERR_INVALID_ARG; }
@@ -424,10 +437,11 @@ static int check_common(const deer_model *m, const deer_forcing *f, int B, int T
 static int check_quasi(const deer_model *m, const deer_forcing *f, int B, int T) {
     int rc = check_common(m, f, B, T);
     if (rc) return rc;
-    if (m->kind != DEER_PLRNN) {
-        set_error("quasi-DEER is built for the vanilla PLRNN (kind DEER_PLRNN) only");
+    if (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN) {
+        set_error("quasi-DEER is built for the PLRNN kinds only");
         return DEER_ERR_INVALID_ARG;
     }
+    if (m->kind == DEER_SHPLRNN) return check_shallow_limits(m);
     return DEER_OK;
 }
 
@@ -771,23 +785,34 @@ static int solve_quasi(const deer_model *m, const deer_forcing *f, const deer_so
                        const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
                        void *ws, size_t ws_bytes, hipStream_t st) {
     size_t need = 0;
-    carve_quasi(nullptr, B, T, m->M, DEER_OP_SOLVE, &need);
+    const int L = quasi_L(m);
+    carve_quasi(nullptr, B, T, m->M, L, DEER_OP_SOLVE, &need);
     int rc = check_ws(ws, ws_bytes, need);
     if (rc) return rc;
-    QuasiWs w = carve_quasi(ws, B, T, m->M, DEER_OP_SOLVE, &need);
+    QuasiWs w = carve_quasi(ws, B, T, m->M, L, DEER_OP_SOLVE, &need);
     PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
+    ShArgs sa{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
     if ((rc = init_guess(o, B, T, m->M, f->n_forced, x, z, st))) return rc;
     std::vector<int> act(B, 1), it(B, 0);
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
     auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *,
                       uint32_t) -> int {
-        return launch_qdeer_update(a, zb, za, zsel, dact, gam, w.rhs, w.coef, w.P, w.v, w.carry, w.ctl.chain_bits, w.C,
-                                   w.ncs, st);
+        if (L == 0)
+            return launch_qdeer_update(a, zb, za, zsel, dact, gam, w.rhs, w.coef, w.P, w.v, w.carry,
+                                       w.ctl.chain_bits, w.C, w.ncs, st);
+        // shallow: residual and hidden-unit masks, then the diagonal coefficients from the masks
+        int r;
+        if ((r = launch_resjac_shplrnn(sa, zb, za, zsel, nullptr, w.rhs, w.masks, dact, st))) return r;
+        if ((r = launch_qdeer_shdiag(sa, w.masks, dact, gam, w.coef, st))) return r;
+        return launch_qdeer_scan_fwd(B, T, m->M, x, f->n_forced, zb, za, zsel, dact, w.rhs, w.coef, w.P, w.v, w.carry,
+                                     w.ctl.chain_bits, w.C, w.ncs, st);
     };
     if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ncs, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
-        if ((rc = launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
+        rc = L == 0 ? launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st)
+                    : launch_resjac_shplrnn(sa, z, nullptr, nullptr, nullptr, nullptr, masks, nullptr, st);
+        if (rc) return rc;
     }
     return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
 }
@@ -1034,11 +1059,25 @@ int deer_adjoint_quasi(const deer_model *m, const deer_forcing *f, int B, int T,
     if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
     hipStream_t st = (hipStream_t)stream;
     size_t need = 0;
-    carve_quasi(nullptr, B, T, m->M, DEER_OP_ADJOINT, &need);
+    const int L = quasi_L(m);
+    carve_quasi(nullptr, B, T, m->M, L, DEER_OP_ADJOINT, &need);
     if ((rc = check_ws(ws, ws_bytes, need))) return rc;
-    QuasiWs w = carve_quasi(ws, B, T, m->M, DEER_OP_ADJOINT, &need);
+    QuasiWs w = carve_quasi(ws, B, T, m->M, L, DEER_OP_ADJOINT, &need);
     PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
     const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
+    if (L > 0) {
+        // shallow: masks and coefficients at z, the reverse scan writes lam, then the shallow
+        // gradient kernel (dA, dW1, dW2, dh1, dh2) from it
+        ShArgs sa{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
+        float *lo = lam ? lam : w.lam;
+        if ((rc = launch_resjac_shplrnn(sa, z, nullptr, nullptr, nullptr, nullptr, w.masks, nullptr, st))) return rc;
+        if ((rc = launch_qdeer_shdiag(sa, w.masks, nullptr, nullptr, w.coef, st))) return rc;
+        if ((rc = launch_qdeer_scan_rev(a, g, scale, z, w.coef, w.P, w.v, w.carry, lo, nullptr, w.C, w.ncs, st)))
+            return rc;
+        if (grads && (grads->A || grads->W || grads->W2 || grads->h || grads->h2))
+            return launch_grads_shplrnn(sa, z, lo, w.masks, w.part, grads, st);
+        return DEER_OK;
+    }
     if ((rc = launch_qdeer_adjoint(a, g, scale, z, w.coef, w.P, w.v, w.carry, lam, w.gpart, w.C, w.ncs, st))) return rc;
     if (grads && (grads->A || grads->W || grads->h))
         return launch_reduce_gpart(w.gpart, B * w.ncs, w.MP, m->M, grads->A, grads->W, grads->h, w.gpart2, st);
@@ -1050,7 +1089,7 @@ size_t deer_quasi_workspace_bytes(const deer_model *m, int B, int T, int op) {
     if (check_quasi(m, &f, B, T) != DEER_OK) return 0;
     if (op != DEER_OP_SOLVE && op != DEER_OP_ADJOINT) return 0;
     size_t bytes = 0;
-    carve_quasi(nullptr, B, T, m->M, op, &bytes);
+    carve_quasi(nullptr, B, T, m->M, quasi_L(m), op, &bytes);
     return bytes;
 }
 

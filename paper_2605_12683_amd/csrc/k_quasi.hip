@@ -321,7 +321,7 @@ __global__ __launch_bounds__(64) void k_qdeer_fixup_fwd(const float *__restrict_
 // z~_s of the same trajectory (the ReLU row of every step through LDS):
 //   gpart[id][i][j] (j < MP) = sum lam_i relu(z~_j),  [MP] = sum lam_i z~_i,  [MP+1] = sum lam_i
 // ---------------------------------------------------------------------------------------
-template <int MP>
+template <int MP, bool GR>
 __global__ __launch_bounds__(64) void k_qdeer_fixup_rev(const float *__restrict__ coef, const float *__restrict__ g,
                                                         float seed_scale, float alpha, int N,
                                                         const float *__restrict__ x, const float *__restrict__ z0,
@@ -360,12 +360,13 @@ __global__ __launch_bounds__(64) void k_qdeer_fixup_rev(const float *__restrict_
                                                                x[((size_t)b * (T + 1) + s + 1) * N + i]))
                            : 0.f;
             }
-            zt = forced_state(x, z0, z, b, s, i, T, M, N, alpha);
+            if (GR) zt = forced_state(x, z0, z, b, s, i, T, M, N, alpha);
             L = fmaf(cv, L, gv);
             if (lam) lam[(base + s) * M + i] = L;
             ga = fmaf(L, zt, ga);
             gh += L;
         }
+        if (!GR) continue;
         lds[lane] = (st && zt > 0.f) ? zt : 0.f;
         wave_lds_sync();
         const float4 *l4 = reinterpret_cast<const float4 *>(lds + n * MP);
@@ -380,12 +381,67 @@ __global__ __launch_bounds__(64) void k_qdeer_fixup_rev(const float *__restrict_
         }
         wave_lds_sync();
     }
-    if (!in) return;
+    if (!GR || !in) return;
     float *gp = gpart + ((size_t)id * MP + i) * (MP + 2);
 #pragma unroll
     for (int j = 0; j < MP; ++j) gp[j] = gw[j];
     gp[MP] = ga;
     gp[MP + 1] = gh;
+}
+
+// ---------------------------------------------------------------------------------------
+// Shallow PLRNN coefficients: coef_s[i] = gamma_b (A_i + sum_l W1_il m_{s,l} W2_li) p_i, the
+// diagonal of J_F = diag(A) + W1 diag(m) W2 times P_alpha, from the hidden-unit ReLU masks of
+// step s.  Block = (tile of steps, sequence b): C_il = W1_il W2_li in LDS, threads = (row,
+// latent); a converged sequence's blocks exit at once.
+// ---------------------------------------------------------------------------------------
+constexpr int QSR = 256;   // threads per block
+
+__global__ __launch_bounds__(QSR) void k_qdeer_shdiag(const float *__restrict__ A, const float *__restrict__ W1,
+                                                     const float *__restrict__ W2, float alpha, int N,
+                                                     const uint32_t *__restrict__ masks, const int *__restrict__ active,
+                                                     const float *__restrict__ gamma, float *__restrict__ coef, int T,
+                                                     int M, int L) {
+    extern __shared__ float Cs[];   // [M][L]
+    const int b = blockIdx.y;
+    if (active && !active[b]) return;
+    for (int e = threadIdx.x; e < M * L; e += QSR) {
+        const int i = e / L, l = e % L;
+        Cs[e] = W1[i * L + l] * W2[l * M + i];
+    }
+    __syncthreads();
+    const int LW = (L + 31) / 32;
+    const float gm = gamma ? gamma[b] : 1.f;
+    const int rows = QSR / M;   // steps handled at once (M <= 64)
+    const int r = threadIdx.x / M, i = threadIdx.x % M;
+    if (r >= rows) return;
+    const float Ai = A[i], pi = i < N ? __fsub_rn(1.0f, alpha) : 1.0f;
+    const float *Ci = Cs + i * L;
+    for (int s = blockIdx.x * rows + r; s < T; s += gridDim.x * rows) {
+        const uint32_t *mw = masks + ((size_t)b * T + s) * LW;
+        float d = 0.f;
+        for (int w = 0; w < LW; ++w) {
+            const uint32_t bits = mw[w];
+            const float *cw = Ci + 32 * w;
+            const int nb = min(32, L - 32 * w);
+            for (int j = 0; j < nb; ++j)
+                if ((bits >> j) & 1u) d += cw[j];
+        }
+        coef[((size_t)b * T + s) * M + i] = gm * ((Ai + d) * pi);
+    }
+}
+
+int launch_qdeer_shdiag(const ShArgs &a, const uint32_t *masks, const int *active, const float *gamma, float *coef,
+                        hipStream_t st) {
+    const int rows = QSR / a.M;
+    long gx = (a.T + rows - 1) / rows;
+    const long cap = (2048L + a.B - 1) / a.B;
+    if (gx > cap) gx = cap;
+    KTimer kt("k_qdeer_shdiag", st);
+    hipLaunchKernelGGL(k_qdeer_shdiag, dim3((unsigned)gx, (unsigned)a.B), dim3(QSR), (size_t)a.M * a.L * sizeof(float),
+                       st, a.A, a.W1, a.W2, a.alpha, a.N, masks, active, gamma, coef, a.T, a.M, a.L);
+    DEER_LAUNCH_CHECK("k_qdeer_shdiag");
+    return DEER_OK;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -417,8 +473,6 @@ int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zs
                         const float *gamma, float *rhs, float *coef, float *P, float *v, float *carry,
                         uint32_t *chain_bits, int C, int ncs, hipStream_t st) {
     const int MP = q_padded(a.M);
-    const int nchains = a.B * ncs;
-    const int gridc = (nchains + 64 / MP - 1) / (64 / MP);
     {
         KTimer kt("k_qdeer_resdiag", st);
         const dim3 grid = q_grid_rows(a.B, a.T, MP);
@@ -429,11 +483,21 @@ int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zs
 #undef RD
     }
     DEER_LAUNCH_CHECK("k_qdeer_resdiag");
+    return launch_qdeer_scan_fwd(a.B, a.T, a.M, a.x, a.N, z, zalt, zsel, active, rhs, coef, P, v, carry, chain_bits, C,
+                                 ncs, st);
+}
+
+int launch_qdeer_scan_fwd(int B, int T, int M, const float *x, int N, float *z, float *zalt, const int *zsel,
+                          const int *active, const float *rhs, const float *coef, float *P, float *v, float *carry,
+                          uint32_t *chain_bits, int C, int ncs, hipStream_t st) {
+    const int MP = q_padded(M);
+    const int nchains = B * ncs;
+    const int gridc = (nchains + 64 / MP - 1) / (64 / MP);
     {
         KTimer kt("k_qdeer_chunk", st);
 #define CK(MPV) \
-    hipLaunchKernelGGL((k_qdeer_chunk<MPV, false>), dim3(gridc), dim3(64), 0, st, (const float *)coef, (const float *)rhs, \
-                       -1.f, (const float *)nullptr, a.x, 0.f, a.N, active, P, v, a.B, a.T, a.M, C, ncs)
+    hipLaunchKernelGGL((k_qdeer_chunk<MPV, false>), dim3(gridc), dim3(64), 0, st, coef, rhs, -1.f, (const float *)nullptr, \
+                       x, 0.f, N, active, P, v, B, T, M, C, ncs)
         if (MP == 16) CK(16); else if (MP == 32) CK(32); else CK(64);
 #undef CK
     }
@@ -441,8 +505,8 @@ int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zs
     {
         KTimer kt("k_qdeer_carry", st);
 #define CR(MPV) \
-    hipLaunchKernelGGL((k_qdeer_carry<MPV, false>), dim3(a.B), dim3(1024), 0, st, (const float *)P, (const float *)v, carry, \
-                       active, a.M, ncs)
+    hipLaunchKernelGGL((k_qdeer_carry<MPV, false>), dim3(B), dim3(1024), 0, st, (const float *)P, (const float *)v, carry, \
+                       active, M, ncs)
         if (MP == 16) CR(16); else if (MP == 32) CR(32); else CR(64);
 #undef CR
     }
@@ -450,8 +514,8 @@ int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zs
     {
         KTimer kt("k_qdeer_fixup_fwd", st);
 #define FX(MPV) \
-    hipLaunchKernelGGL((k_qdeer_fixup_fwd<MPV>), dim3(gridc), dim3(64), 0, st, (const float *)coef, (const float *)rhs, \
-                       (const float *)carry, z, zalt, zsel, chain_bits, active, a.B, a.T, a.M, C, ncs)
+    hipLaunchKernelGGL((k_qdeer_fixup_fwd<MPV>), dim3(gridc), dim3(64), 0, st, coef, rhs, (const float *)carry, z, zalt, \
+                       zsel, chain_bits, active, B, T, M, C, ncs)
         if (MP == 16) FX(16); else if (MP == 32) FX(32); else FX(64);
 #undef FX
     }
@@ -462,8 +526,6 @@ int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zs
 int launch_qdeer_adjoint(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *coef, float *P,
                          float *v, float *carry, float *lam, float *gpart, int C, int ncs, hipStream_t st) {
     const int MP = q_padded(a.M);
-    const int nchains = a.B * ncs;
-    const int gridc = (nchains + 64 / MP - 1) / (64 / MP);
     {
         KTimer kt("k_qdeer_resdiag", st);
         const dim3 grid = q_grid_rows(a.B, a.T, MP);
@@ -475,10 +537,18 @@ int launch_qdeer_adjoint(const PlrnnArgs &a, const float *g, float seed_scale, c
 #undef RD
     }
     DEER_LAUNCH_CHECK("k_qdeer_resdiag<rev>");
+    return launch_qdeer_scan_rev(a, g, seed_scale, z, coef, P, v, carry, lam, gpart, C, ncs, st);
+}
+
+int launch_qdeer_scan_rev(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, const float *coef,
+                          float *P, float *v, float *carry, float *lam, float *gpart, int C, int ncs, hipStream_t st) {
+    const int MP = q_padded(a.M);
+    const int nchains = a.B * ncs;
+    const int gridc = (nchains + 64 / MP - 1) / (64 / MP);
     {
         KTimer kt("k_qdeer_chunk", st);
 #define CK(MPV) \
-    hipLaunchKernelGGL((k_qdeer_chunk<MPV, true>), dim3(gridc), dim3(64), 0, st, (const float *)coef, g, 1.f, z, a.x, \
+    hipLaunchKernelGGL((k_qdeer_chunk<MPV, true>), dim3(gridc), dim3(64), 0, st, coef, g, 1.f, z, a.x, \
                        seed_scale, a.N, (const int *)nullptr, P, v, a.B, a.T, a.M, C, ncs)
         if (MP == 16) CK(16); else if (MP == 32) CK(32); else CK(64);
 #undef CK
@@ -495,10 +565,12 @@ int launch_qdeer_adjoint(const PlrnnArgs &a, const float *g, float seed_scale, c
     DEER_LAUNCH_CHECK("k_qdeer_carry<rev>");
     {
         KTimer kt("k_qdeer_fixup_rev", st);
-#define FX(MPV) \
-    hipLaunchKernelGGL((k_qdeer_fixup_rev<MPV>), dim3(gridc), dim3(64), 0, st, (const float *)coef, g, seed_scale, a.alpha, \
-                       a.N, a.x, a.z0, z, (const float *)carry, lam, gpart, a.B, a.T, a.M, C, ncs)
-        if (MP == 16) FX(16); else if (MP == 32) FX(32); else FX(64);
+#define FX(MPV, GRV) \
+    hipLaunchKernelGGL((k_qdeer_fixup_rev<MPV, GRV>), dim3(gridc), dim3(64), 0, st, coef, g, seed_scale, \
+                       a.alpha, a.N, a.x, a.z0, z, (const float *)carry, lam, gpart, a.B, a.T, a.M, C, ncs)
+#define FXG(GRV) if (MP == 16) FX(16, GRV); else if (MP == 32) FX(32, GRV); else FX(64, GRV);
+        if (gpart) { FXG(true) } else { FXG(false) }
+#undef FXG
 #undef FX
     }
     DEER_LAUNCH_CHECK("k_qdeer_fixup_rev");

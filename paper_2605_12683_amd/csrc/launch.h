@@ -118,6 +118,16 @@ int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zs
                         uint32_t *chain_bits, int C, int ncs, hipStream_t st);
 int launch_qdeer_adjoint(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *coef, float *P,
                          float *v, float *carry, float *lam, float *gpart, int C, int ncs, hipStream_t st);
+// the model-independent parts: the forward scan + fix-up from (rhs = r, coef), and the reverse
+// scan from coef (gpart null: no vanilla gradient partials, lam written); shallow-PLRNN
+// coefficients from the hidden-unit masks (M L <= 8192)
+int launch_qdeer_scan_fwd(int B, int T, int M, const float *x, int N, float *z, float *zalt, const int *zsel,
+                          const int *active, const float *rhs, const float *coef, float *P, float *v, float *carry,
+                          uint32_t *chain_bits, int C, int ncs, hipStream_t st);
+int launch_qdeer_scan_rev(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, const float *coef,
+                          float *P, float *v, float *carry, float *lam, float *gpart, int C, int ncs, hipStream_t st);
+int launch_qdeer_shdiag(const ShArgs &a, const uint32_t *masks, const int *active, const float *gamma, float *coef,
+                        hipStream_t st);
 
 // dense stored-Jacobian scan (mode: 0 Newton fix-up, 1 bare forward scan, 2 reverse)
 int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,

@@ -60,7 +60,9 @@ def test_workspace_queries(lib):
     bad = _b.deer_model(_b.DEER_PLRNN, 65, 0, m.A, m.W, None, None, None)
     assert lib.deer_workspace_bytes(ctypes.byref(bad), 4, 16, _b.DEER_OP_SOLVE) == 0
     sh, _keep2 = _vanilla_model(4, _b.DEER_SHPLRNN)
-    assert lib.deer_quasi_workspace_bytes(ctypes.byref(sh), 4, 16, _b.DEER_OP_SOLVE) == 0   # vanilla only
+    assert lib.deer_quasi_workspace_bytes(ctypes.byref(sh), 4, 16, _b.DEER_OP_SOLVE) > 0
+    dg = _b.deer_model(_b.DEER_DIAG_SSM, 4, 3, m.A, m.W, None, None, None)
+    assert lib.deer_quasi_workspace_bytes(ctypes.byref(dg), 4, 16, _b.DEER_OP_SOLVE) == 0   # PLRNN kinds only
 
 
 def test_argument_errors_before_device_work(lib):
@@ -77,10 +79,10 @@ def test_argument_errors_before_device_work(lib):
     st = lib.deer_adjoint_quasi(ctypes.byref(m), ctypes.byref(f), 2, 8, None, None, None, None, None,
                                 ctypes.byref(gs), None, 0, None)
     assert st == _b.DEER_ERR_INVALID_ARG                # x and z are required
-    sh, _keep2 = _vanilla_model(4, _b.DEER_SHPLRNN)
-    st = lib.deer_solve_quasi(ctypes.byref(sh), ctypes.byref(f), ctypes.byref(o), 2, 8, None, None, None, None,
+    dg = _b.deer_model(_b.DEER_DIAG_SSM, 4, 3, m.A, m.W, None, None, None)
+    st = lib.deer_solve_quasi(ctypes.byref(dg), ctypes.byref(f), ctypes.byref(o), 2, 8, None, None, None, None,
                               None, None, None, 0, None)
-    assert st == _b.DEER_ERR_INVALID_ARG and b"vanilla" in lib.deer_last_error()
+    assert st == _b.DEER_ERR_INVALID_ARG and b"PLRNN" in lib.deer_last_error()
 
 
 def test_status_strings(lib):

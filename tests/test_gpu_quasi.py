@@ -118,3 +118,46 @@ def test_quasi_workload2_full_size():
     gr = O.param_grads(m, c.x, z32, c.alpha, c.n_obs, lam, mask_precision="float32")
     for k, v in out["grads"].items():
         assert rel_inf(v.cpu().numpy(), gr[k]) < TOL, k
+
+
+# ---- shallow PLRNN (the model of the paper's quasi-DEER ablation: M = 5, L = 50) ----------
+
+SH_SIZES = [(5, 50, 3, 1, 300), (3, 7, 3, 2, 129), (8, 32, 2, 2, 700), (32, 256, 32, 1, 1024)]
+
+
+def _sh_case(M, L, N, B, T, alpha, seed):
+    return W.random_shplrnn_case(M, L, N, B, T, alpha, seed, w_norm=0.2, a_range=(0.3, 0.75))
+
+
+@pytest.mark.parametrize("M,L,N,B,T", SH_SIZES)
+def test_quasi_shallow_first_update_and_rollout(M, L, N, B, T):
+    c = _sh_case(M, L, N, B, T, 0.15, 400 + M + L)
+    m = oracle_model(c)
+    say("deer_solve_quasi shallow first update", M, L, N, B, T)
+    res = D.deer_solve_quasi(m, c.x, c.alpha, N, fixed_iters=1)
+    ref = O.newton(m, c.x, c.alpha, N, fixed_iters=1, quasi=True)
+    assert rel_inf(res["z"].cpu().numpy(), ref["z"]) < TOL
+    say("deer_solve_quasi shallow to tolerance", M, L, N, B, T)
+    res = D.deer_solve_quasi(m, c.x, c.alpha, N, tol=1e-5, max_iter=T + 2)
+    assert res["status"] == 0
+    assert rel_inf(res["z"].cpu().numpy(), O.rollout(m, c.x, c.alpha, N)) < TOL
+    print(f"[gpu-case] shallow quasi updates {res['iters']}", flush=True)
+
+
+@pytest.mark.parametrize("M,L,N,B,T", SH_SIZES)
+@pytest.mark.parametrize("user_g", [False, True])
+def test_quasi_shallow_adjoint_and_gradients(M, L, N, B, T, user_g):
+    c = _sh_case(M, L, N, B, T, 0.15, 410 + M + L)
+    m = oracle_model(c)
+    z32 = O.rollout(m, c.x, c.alpha, N).astype(np.float32)
+    g = np.random.default_rng(M + L).standard_normal((B, T, M)).astype(np.float32) if user_g else None
+    say("deer_adjoint_quasi shallow", M, L, N, B, T, user_g)
+    out = D.deer_adjoint_quasi(m, c.x, z32, c.alpha, N, g=g)
+    lam = O.adjoint(m, c.x, z32, c.alpha, N, g=g, mask_precision="float32", quasi=True)
+    assert rel_inf(out["lam"].cpu().numpy(), lam) < TOL
+    gr = O.param_grads(m, c.x, z32, c.alpha, N, lam, mask_precision="float32")
+    for k, v in out["grads"].items():
+        assert rel_inf(v.cpu().numpy(), gr[k]) < TOL, k
+    out2 = D.deer_adjoint_quasi(m, c.x, z32, c.alpha, N, g=g, want_lam=False)
+    for k, v in out2["grads"].items():
+        assert rel_inf(v.cpu().numpy(), gr[k]) < TOL, k

@@ -60,6 +60,15 @@ def forcing_weights(M: int, n_forced: int, alpha: float) -> np.ndarray:
     return a
 
 
+def forcing_schedule(M: int, n_forced: int, alpha: float, T: int, T_w: int = 0) -> np.ndarray:
+    """a_k of the forced input z~_k for k = 0..T-1, shape [T, M]: alpha on the observed latents,
+    and 1 there during the latent warm-up, k = 1..T_w (Alg. GTF-DEER: P_1 and the full forcing
+    for t <= T_w; latent state warm-up paragraph).  Row 0 is unused (z~_0 = z_0)."""
+    a = np.tile(forcing_weights(M, n_forced, alpha), (max(T, 1), 1))
+    a[1:T_w + 1, :n_forced] = 1.0
+    return a
+
+
 def teacher_states(x: np.ndarray, M: int) -> np.ndarray:
     """zbar_t = B^+ x_t = [x_t; 0] for t = 0..T (Alg. GTF-DEER, forcing targets)."""
     x = np.asarray(x, f64)
@@ -78,10 +87,11 @@ def initial_state(x: np.ndarray, M: int, z0=None) -> np.ndarray:
 
 def forced_states(z: np.ndarray, zbar: np.ndarray, a: np.ndarray, z0: np.ndarray) -> np.ndarray:
     """z~_{t-1} = (1 - a) z_{t-1} + a zbar_{t-1} for t >= 2 and z~_0 = z_0 (eqs. GTF,
-    error_forcing; GTF-DEER residual for step 1)."""
+    error_forcing; GTF-DEER residual for step 1).  a is [M] or per step [T, M]."""
     zt = np.zeros_like(z)
     zt[:, 0] = z0
-    zt[:, 1:] = (1.0 - a) * z[:, :-1] + a * zbar[:, 1:-1]
+    ak = a if a.ndim == 1 else a[1:]
+    zt[:, 1:] = (1.0 - ak) * z[:, :-1] + ak * zbar[:, 1:-1]
     return zt
 
 
@@ -120,7 +130,7 @@ def activation_mask(model: dict, zt: np.ndarray) -> np.ndarray:
 
 
 def activation_mask_fp32(model: dict, z: np.ndarray, x: np.ndarray, alpha: float, n_forced: int,
-                         z0=None) -> np.ndarray:
+                         z0=None, T_w: int = 0) -> np.ndarray:
     """The same ReLU decision taken in float32, in the order the GPU kernels take it.
 
     Where floating point decides an integer both sides decide in the same
@@ -132,14 +142,15 @@ def activation_mask_fp32(model: dict, z: np.ndarray, x: np.ndarray, alpha: float
     f = np.float32
     z = np.asarray(z, f)
     Bn, T, M = z.shape
-    a32 = np.zeros(M, f)
-    a32[:n_forced] = f(alpha)
+    a32 = np.zeros((T, M), f)
+    a32[:, :n_forced] = f(alpha)
+    a32[1:T_w + 1, :n_forced] = f(1.0)
     p32 = (f(1.0) - a32).astype(f)
     zbar = np.zeros((Bn, T + 1, M), f)
     zbar[:, :, :x.shape[2]] = np.asarray(x, f)
     zt = np.zeros((Bn, T, M), f)
     zt[:, 0] = zbar[:, 0] if z0 is None else np.asarray(z0, f)
-    zt[:, 1:] = (p32 * z[:, :-1]).astype(f) + (a32 * zbar[:, 1:-1]).astype(f)
+    zt[:, 1:] = (p32[1:] * z[:, :-1]).astype(f) + (a32[1:] * zbar[:, 1:-1]).astype(f)
     if model["kind"] == "plrnn":
         return zt > 0
     W2 = np.asarray(model["W2"], f)
@@ -193,20 +204,21 @@ def forced_jacobians(model: dict, mask: np.ndarray, a: np.ndarray) -> np.ndarray
 # O1: sequential GTF rollout (Alg. initial value / trajectory matching with GTF)
 # --------------------------------------------------------------------------------------
 
-def rollout(model: dict, x: np.ndarray, alpha: float, n_forced: int, z0=None) -> np.ndarray:
+def rollout(model: dict, x: np.ndarray, alpha: float, n_forced: int, z0=None, T_w: int = 0) -> np.ndarray:
     """z_t = F(z~_{t-1}) for t = 1..T, one step at a time.  This is the unique
-    zero-residual trajectory that DEER converges to."""
+    zero-residual trajectory that DEER converges to.  T_w: latent warm-up (full forcing of
+    the observed latents for z~_1..z~_{T_w})."""
     model = _model64(model)
     x = np.asarray(x, f64)
     Bn, T1, _ = x.shape
     T = T1 - 1
     M = np.asarray(model["A"]).shape[0]
-    a = forcing_weights(M, n_forced, alpha)
+    a = forcing_schedule(M, n_forced, alpha, T, T_w)
     zbar = teacher_states(x, M)
     zprev = initial_state(x, M, z0)
     z = np.zeros((Bn, T, M), f64)
     for t in range(1, T + 1):
-        ztil = zprev if t == 1 else (1.0 - a) * zprev + a * zbar[:, t - 1]
+        ztil = zprev if t == 1 else (1.0 - a[t - 1]) * zprev + a[t - 1] * zbar[:, t - 1]
         zprev = model_map(model, ztil)
         z[:, t - 1] = zprev
     return z
@@ -245,13 +257,14 @@ def reverse_affine_recurrence(apply_JT, g: np.ndarray) -> np.ndarray:
 # O2: explicit GTF-DEER Newton loop (Alg. GTF-DEER; eq. GTF_DEER_update)
 # --------------------------------------------------------------------------------------
 
-def residual_and_masks(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, z0=None):
+def residual_and_masks(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, z0=None,
+                       T_w: int = 0):
     """r_t = z_t - F(z~_{t-1}) (eq. GTF_residual) together with F and the masks at z~."""
     model = _model64(model)
     x = np.asarray(x, f64)
     z = np.asarray(z, f64)
     M = z.shape[2]
-    a = forcing_weights(M, n_forced, alpha)
+    a = forcing_schedule(M, n_forced, alpha, z.shape[1], T_w)
     zbar = teacher_states(x, M)
     zt = forced_states(z, zbar, a, initial_state(x, M, z0))
     F = model_map(model, zt)
@@ -260,7 +273,7 @@ def residual_and_masks(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, 
 
 def newton(model: dict, x: np.ndarray, alpha: float, n_forced: int, *, z0=None, init: str = "teacher",
            z_init=None, tol: float = 1e-5, max_iter: int = 500, fixed_iters: int = 0, history: bool = False,
-           gamma: float = 1.0, quasi: bool = False):
+           gamma: float = 1.0, quasi: bool = False, T_w: int = 0):
     """GTF-DEER forward solve.  Each update linearises at z^(k): Delta_t =
     J~_t Delta_{t-1} - r_t, Delta_0 = 0, solved here by the sequential recursion,
     then z^(k+1) = z^(k) + Delta.  Returns dict(z, iters, norms, status[, history]).
@@ -271,13 +284,15 @@ def newton(model: dict, x: np.ndarray, alpha: float, n_forced: int, *, z0=None, 
 
     quasi: quasi-DEER, J~_t replaced by its diagonal diag(J_F(z~_{t-1})) P_alpha (the
     diagonal approximation discussed with eq. DEER_update), Delta_t = d_t * Delta_{t-1} - r_t;
-    the fixed point is the same."""
+    the fixed point is the same.
+
+    T_w: latent warm-up, z~_k and J~_{k+1} with full forcing (P_1) for k = 1..T_w."""
     model = _model64(model)
     x = np.asarray(x, f64)
     Bn, T1, _ = x.shape
     T = T1 - 1
     M = np.asarray(model["A"]).shape[0]
-    a = forcing_weights(M, n_forced, alpha)
+    a = forcing_schedule(M, n_forced, alpha, T, T_w)
     p = 1.0 - a
     zbar = teacher_states(x, M)
     z0v = initial_state(x, M, z0)
@@ -308,7 +323,7 @@ def newton(model: dict, x: np.ndarray, alpha: float, n_forced: int, *, z0=None, 
             dg = jacobian_diagonal(model, mask) * p
             delta = affine_recurrence(lambda kk, v: gamma * (dg[:, kk] * v), -r)
         else:
-            delta = affine_recurrence(lambda kk, v: gamma * jvp(model, mask[:, kk], p * v), -r)
+            delta = affine_recurrence(lambda kk, v: gamma * jvp(model, mask[:, kk], p[kk] * v), -r)
         e = np.abs(delta).reshape(Bn, -1).max(axis=1) if T > 0 else np.zeros(Bn)
         e = np.where(np.isnan(delta).reshape(Bn, -1).any(axis=1), np.nan, e)
         upd = active if fixed_iters == 0 else np.ones(Bn, bool)
@@ -337,30 +352,31 @@ def newton(model: dict, x: np.ndarray, alpha: float, n_forced: int, *, z0=None, 
 # O3: loss seed, IFT adjoint and parameter gradients (gradients appendix)
 # --------------------------------------------------------------------------------------
 
-def mse_loss(z: np.ndarray, x: np.ndarray) -> float:
-    """Batch mean of (1/(N T)) sum_t ||x_t - B z_t||^2 (eq. mse_loss_series)."""
+def mse_loss(z: np.ndarray, x: np.ndarray, T_w: int = 0) -> float:
+    """Batch mean of (1/(N (T - T_w))) sum_{t > T_w} ||x_t - B z_t||^2 (eqs. mse_loss_series,
+    mse_loss_warmup: the warm-up states are excluded)."""
     z = np.asarray(z, f64)
     x = np.asarray(x, f64)
     Bn, T, _ = z.shape
     N = x.shape[2]
-    return float(((z[:, :, :N] - x[:, 1:]) ** 2).sum() / (Bn * N * T))
+    return float(((z[:, T_w:, :N] - x[:, 1 + T_w:]) ** 2).sum() / (Bn * N * (T - T_w)))
 
 
-def mse_seed(z: np.ndarray, x: np.ndarray) -> np.ndarray:
-    """dL/dz_t = 2/(B N T) B^T (B z_t - x_t), t = 1..T."""
+def mse_seed(z: np.ndarray, x: np.ndarray, T_w: int = 0) -> np.ndarray:
+    """dL/dz_t = 2/(B N (T - T_w)) B^T (B z_t - x_t) for t = T_w+1..T, zero in the warm-up."""
     z = np.asarray(z, f64)
     x = np.asarray(x, f64)
     Bn, T, M = z.shape
     N = x.shape[2]
     g = np.zeros((Bn, T, M), f64)
-    g[:, :, :N] = 2.0 / (Bn * N * T) * (z[:, :, :N] - x[:, 1:])
+    g[:, T_w:, :N] = 2.0 / (Bn * N * (T - T_w)) * (z[:, T_w:, :N] - x[:, 1 + T_w:])
     return g
 
 
-def _masks_at(model, x, z, alpha, n_forced, z0, mask_precision):
-    r, F, mask64, zt = residual_and_masks(model, x, z, alpha, n_forced, z0)
+def _masks_at(model, x, z, alpha, n_forced, z0, mask_precision, T_w=0):
+    r, F, mask64, zt = residual_and_masks(model, x, z, alpha, n_forced, z0, T_w)
     if mask_precision == "float32":
-        mask = activation_mask_fp32(model, z, x, alpha, n_forced, z0)
+        mask = activation_mask_fp32(model, z, x, alpha, n_forced, z0, T_w)
     elif mask_precision == "float64":
         mask = mask64
     else:
@@ -369,7 +385,7 @@ def _masks_at(model, x, z, alpha, n_forced, z0, mask_precision):
 
 
 def adjoint(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, *, z0=None,
-            g=None, mask_precision: str = "float64", quasi: bool = False) -> np.ndarray:
+            g=None, mask_precision: str = "float64", quasi: bool = False, T_w: int = 0) -> np.ndarray:
     """lam = dL/dz by the backward recursion lam_T = g_T, lam_{t-1} = J~_t^T lam_t + g_{t-1}
     (eqs. adjoint_eq, backward_recursion with lam = -v).  J~_t is taken at z~_{t-1} of
     the given trajectory z (normally the converged one).
@@ -380,24 +396,24 @@ def adjoint(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: i
     model = _model64(model)
     z = np.asarray(z, f64)
     M = z.shape[2]
-    p = 1.0 - forcing_weights(M, n_forced, alpha)
-    mask, _ = _masks_at(model, x, z, alpha, n_forced, z0, mask_precision)
-    g = mse_seed(z, x) if g is None else np.asarray(g, f64)
+    p = 1.0 - forcing_schedule(M, n_forced, alpha, z.shape[1], T_w)
+    mask, _ = _masks_at(model, x, z, alpha, n_forced, z0, mask_precision, T_w)
+    g = mse_seed(z, x, T_w) if g is None else np.asarray(g, f64)
     if quasi:
         dg = jacobian_diagonal(model, mask) * p
         return reverse_affine_recurrence(lambda k, w: dg[:, k] * w, g)
     # J~^T w = P_alpha J_F^T w
-    return reverse_affine_recurrence(lambda k, w: p * vjp(model, mask[:, k], w), g)
+    return reverse_affine_recurrence(lambda k, w: p[k] * vjp(model, mask[:, k], w), g)
 
 
 def param_grads(model: dict, x: np.ndarray, z: np.ndarray, alpha: float, n_forced: int, lam: np.ndarray, *,
-                z0=None, mask_precision: str = "float64") -> dict:
+                z0=None, mask_precision: str = "float64", T_w: int = 0) -> dict:
     """dL/dtheta = sum_t lam_t^T dF(z~_{t-1})/dtheta (gradients appendix, IFT summary),
     summed directly over every (b, t) in float64."""
     model = _model64(model)
     z = np.asarray(z, f64)
     lam = np.asarray(lam, f64)
-    mask, zt = _masks_at(model, x, z, alpha, n_forced, z0, mask_precision)
+    mask, zt = _masks_at(model, x, z, alpha, n_forced, z0, mask_precision, T_w)
     out = {"A": np.einsum("bti,bti->i", lam, zt, optimize=True)}
     if model["kind"] == "plrnn":
         relu = np.where(mask, zt, 0.0)

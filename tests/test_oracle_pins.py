@@ -335,9 +335,10 @@ def test_adjoint_equals_dense_adjoint_solve(kind):
     assert np.allclose(lam, brute.block_bidiagonal_adjoint_solve(J, g), rtol=1e-12, atol=1e-14)
 
 
-def _torch_bptt(m, x, alpha, N):
+def _torch_bptt(m, x, alpha, N, T_w=0):
     """Independent reverse-mode AD (torch, float64) through the sequential GTF rollout
-    of Alg. 2 and the MSE loss: the BPTT gradient the IFT gradient must equal."""
+    of Alg. 2 and the MSE loss: the BPTT gradient the IFT gradient must equal.  T_w: the
+    first T_w forced inputs fully forced, their states left out of the loss."""
     t = lambda a: torch.tensor(np.asarray(a, np.float64), requires_grad=True)
     P = {k: t(v) for k, v in m.items() if k != "kind"}
     xt = torch.tensor(np.asarray(x, np.float64))
@@ -349,14 +350,18 @@ def _torch_bptt(m, x, alpha, N):
     zbar[:, :, :N] = xt
     prev = zbar[:, 0]
     loss = 0.0
+    aw = a.clone()
+    aw[:N] = 1.0
     for k in range(1, T1):
-        zt = prev if k == 1 else (1 - a) * prev + a * zbar[:, k - 1]
+        ak = aw if k - 1 <= T_w else a
+        zt = prev if k == 1 else (1 - ak) * prev + ak * zbar[:, k - 1]
         if m["kind"] == "plrnn":
             prev = P["A"] * zt + torch.relu(zt) @ P["W"].T + P["h"]
         else:
             prev = P["A"] * zt + torch.relu(zt @ P["W2"].T + P["h2"]) @ P["W1"].T + P["h1"]
-        loss = loss + ((prev[:, :N] - xt[:, k]) ** 2).sum()
-    loss = loss / (Bn * N * (T1 - 1))
+        if k > T_w:
+            loss = loss + ((prev[:, :N] - xt[:, k]) ** 2).sum()
+    loss = loss / (Bn * N * (T1 - 1 - T_w))
     loss.backward()
     return float(loss.detach()), {k: v.grad.numpy() for k, v in P.items()}
 
@@ -580,3 +585,82 @@ def test_quasi_converges_to_rollout_with_prefix_exactness(kind, M, N, alpha):
     hist = O.newton(m, xs, alpha, N, fixed_iters=T, history=True, quasi=True)["history"]
     for k in range(1, T + 1):
         assert np.abs(hist[k][:, :k] - refs[:, :k]).max() < 1e-12, k
+
+
+
+# ------------------------------------------------------------------------------------
+# latent warm-up (Alg. GTF-DEER: P_1 for t <= T_w; the warm-up states left out of the loss)
+# ------------------------------------------------------------------------------------
+
+def test_warmup_prefix_is_driven_by_the_data():
+    """With every latent observed, the warm-up inputs are the data themselves: z_1 = F(z_0),
+    z_t = F(x_{t-1}) for t = 2..T_w + 1; afterwards the forcing is alpha again."""
+    M = N = 4
+    m = _vanilla(M, 61)
+    x = _x(2, 30, N, 62)
+    T_w = 10
+    z = O.rollout(m, x, 0.3, N, T_w=T_w)
+    m64 = {k: (v if k == "kind" else np.asarray(v, np.float64)) for k, v in m.items()}
+    assert np.allclose(z[:, 1:T_w + 1], O.model_map(m64, np.asarray(x[:, 1:T_w + 1], np.float64)), atol=1e-13)
+    assert not np.allclose(z[:, T_w + 1], O.model_map(m64, np.asarray(x[:, T_w + 1], np.float64)))
+    assert np.allclose(O.rollout(m, x, 0.3, N, T_w=0), O.rollout(m, x, 0.3, N))
+
+
+@pytest.mark.parametrize("kind,M,N,alpha,T_w", [("plrnn", 4, 3, 0.2, 7), ("plrnn", 16, 3, 0.2, 25),
+                                                ("shplrnn", 5, 3, 0.15, 12)])
+def test_warmup_newton_reaches_rollout(kind, M, N, alpha, T_w):
+    m = _vanilla(M, 63) if kind == "plrnn" else _shallow(M, 3 * M, 64)
+    x = _x(2, 60, N, 65)
+    ref = O.rollout(m, x, alpha, N, T_w=T_w)
+    res = O.newton(m, x, alpha, N, tol=1e-13, max_iter=200, T_w=T_w)
+    assert res["status"] == "ok"
+    assert np.abs(res["z"] - ref).max() <= 1e-11
+    q = O.newton(m, x, alpha, N, tol=1e-13, max_iter=500, T_w=T_w, quasi=True)
+    assert np.abs(q["z"] - ref).max() <= 1e-11
+
+
+@pytest.mark.parametrize("kind,M,N,alpha,T_w", [("plrnn", 5, 3, 0.2, 6), ("shplrnn", 4, 4, 0.15, 9)])
+def test_warmup_gradient_equals_bptt(kind, M, N, alpha, T_w):
+    """IFT gradient with the warm-up (full forcing, warm-up states out of the loss) equals
+    reverse-mode AD through the sequential rollout."""
+    m = _vanilla(M, 66) if kind == "plrnn" else _shallow(M, 7, 67)
+    x = _x(2, 25, N, 68)
+    z = O.rollout(m, x, alpha, N, T_w=T_w)
+    lam = O.adjoint(m, x, z, alpha, N, T_w=T_w)
+    gr = O.param_grads(m, x, z, alpha, N, lam, T_w=T_w)
+    loss, ref = _torch_bptt(m, x, alpha, N, T_w=T_w)
+    assert abs(O.mse_loss(z, x, T_w=T_w) - loss) <= 1e-12 * max(1.0, abs(loss))
+    for k, v in ref.items():
+        assert np.allclose(gr[k], v, rtol=1e-9, atol=1e-12), k
+
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+def test_warmup_as_two_chained_solves(kind):
+    """The warm-up part and the rest can be solved one after the other: the prefix with
+    alpha = 1, the rest from z_0 := P_1 z_{T_w} + zbar_{T_w}; the adjoint of the rest (MSE seed
+    over its own steps) hands J~_{T_w+1}^T lam_{T_w+1} to the prefix as its only cotangent, and
+    the parameter gradients add."""
+    M, N, alpha, T, T_w = 4, 2, 0.25, 40, 11
+    m = _vanilla(M, 69) if kind == "plrnn" else _shallow(M, 6, 70)
+    x = _x(2, T, N, 71)
+    z = O.rollout(m, x, alpha, N, T_w=T_w)
+    x1, x2 = x[:, :T_w + 1], x[:, T_w:]
+    z1 = O.rollout(m, x1, 1.0, N)
+    zb = np.concatenate([np.asarray(x[:, T_w], np.float64), z1[:, -1, N:]], axis=1)
+    z2 = O.rollout(m, x2, alpha, N, z0=zb)
+    assert np.allclose(np.concatenate([z1, z2], axis=1), z, atol=1e-13)
+    lam = O.adjoint(m, x, z, alpha, N, T_w=T_w)
+    gr = O.param_grads(m, x, z, alpha, N, lam, T_w=T_w)
+    lam2 = O.adjoint(m, x2, z2, alpha, N, z0=zb)
+    # J~_{T_w+1} at the fully forced input zb: P_1 J_F(zb)^T lam2[:, 0]
+    m64 = {k: (v if k == "kind" else np.asarray(v, np.float64)) for k, v in m.items()}
+    p1 = 1.0 - O.forcing_weights(M, N, 1.0)
+    gb = p1 * O.vjp(m64, O.activation_mask(m64, zb), lam2[:, 0])
+    g1 = np.zeros_like(z1)
+    g1[:, -1] = gb
+    lam1 = O.adjoint(m, x1, z1, 1.0, N, g=g1)
+    assert np.allclose(np.concatenate([lam1, lam2], axis=1), lam, rtol=1e-12, atol=1e-15)
+    g_a = O.param_grads(m, x1, z1, 1.0, N, lam1)
+    g_b = O.param_grads(m, x2, z2, alpha, N, lam2, z0=zb)
+    for k in gr:
+        assert np.allclose(g_a[k] + g_b[k], gr[k], rtol=1e-11, atol=1e-14), k

@@ -37,13 +37,13 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def _plrnn_step(D, model, xd, c, ws_s, ws_a):
+def _plrnn_step(D, model, xd, c, ws_s, ws_a, T_w=0):
     res = D.deer_solve(model, xd, c.alpha, c.n_obs, tol=c.tol, max_iter=c.max_iter, fixed_iters=c.fixed_iters,
-                       ws=ws_s, check=False)
+                       ws=ws_s, check=False, T_w=T_w)
     if res["status"] != 0:
         raise RuntimeError(f"deer_solve returned status {res['status']}: {D.load().deer_last_error()}")
     # the step's outputs are the parameter gradients: the adjoint itself is not stored
-    D.deer_adjoint(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a, want_lam=False)
+    D.deer_adjoint(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a, want_lam=False, T_w=T_w)
     return sum(res["iters"])
 
 
@@ -285,6 +285,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--tw", type=int, default=0,
+                    help="PLRNN workloads with a tolerance: latent warm-up of this many steps")
     ap.add_argument("--quasi", action="store_true",
                     help="PLRNN workloads: quasi-DEER (diagonal Jacobians) instead of GTF-DEER")
     ap.add_argument("--fig1a", action="store_true",
@@ -331,9 +333,13 @@ def main():
                                                                Bnd.DEER_OP_ADJOINT))
             step = lambda: _quasi_step(D, model, xd, c, ws_s, ws_a)        # noqa: E731
         else:
-            ws_s = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_SOLVE))
-            ws_a = D._workspace(D.deer_workspace_bytes(model, c.B, c.T, Bnd.DEER_OP_ADJOINT))
-            step = lambda: _plrnn_step(D, model, xd, c, ws_s, ws_a)        # noqa: E731
+            lib = D.load()
+            fw = Bnd.deer_forcing(float(c.alpha), int(c.n_obs), int(args.tw))
+            ws_s = D._workspace(lib.deer_workspace_bytes_ex(ctypes.byref(model.c), ctypes.byref(fw), c.B, c.T,
+                                                            Bnd.DEER_OP_SOLVE, 0))
+            ws_a = D._workspace(lib.deer_workspace_bytes_ex(ctypes.byref(model.c), ctypes.byref(fw), c.B, c.T,
+                                                            Bnd.DEER_OP_ADJOINT, 0))
+            step = lambda: _plrnn_step(D, model, xd, c, ws_s, ws_a, args.tw)   # noqa: E731
     else:
         print(f"workload {c.name}: model kind {c.kind} not supported by this build", file=sys.stderr)
         sys.exit(3)
@@ -392,7 +398,7 @@ def main():
                    "alpha": c.alpha, "tol": c.tol if not c.fixed_iters else None,
                    "fixed_iters": c.fixed_iters or None, "newton_updates_per_step": iters_per_step,
                    "step": ("deer_solve_quasi + deer_adjoint_quasi (quasi-DEER: diagonal Jacobians)" if args.quasi
-                            else "deer_solve + deer_adjoint")},
+                            else "deer_solve + deer_adjoint"), "latent_warmup": args.tw},
         "roofline": roof,
         "kernels": kernels,
     }

@@ -85,6 +85,11 @@ typedef struct {
 typedef struct {
     float alpha;        /* GTF forcing strength in [0, 1] (eq. GTF)                          */
     int n_forced;       /* N: the first N latents are observed and forced, 0 <= N <= M      */
+    int T_w;            /* latent warm-up (Alg. GTF-DEER, latent state warm-up paragraph):
+                           0 <= T_w < T; the forced inputs z~_1..z~_{T_w} use alpha = 1 and
+                           the MSE seed leaves z_1..z_{T_w} out (1 / (N (T - T_w))).  PLRNN
+                           kinds, solves with a tolerance (fixed_iters = 0) only; the
+                           workspace is deer_workspace_bytes_ex(...).                       */
 } deer_forcing;
 
 enum { DEER_INIT_TEACHER = 0, DEER_INIT_ZERO = 1, DEER_INIT_USER = 2 };
@@ -113,8 +118,17 @@ enum { DEER_OP_SOLVE = 0, DEER_OP_ADJOINT = 1 };
 enum { DEER_SCAN_DENSE = 0, DEER_SCAN_DIAG_C64 = 1 };
 
 /* Bytes of workspace `op` (DEER_OP_SOLVE or DEER_OP_ADJOINT) needs for this model and
- * size.  Returns 0 for invalid arguments. */
+ * size (no warm-up).  Returns 0 for invalid arguments. */
 size_t deer_workspace_bytes(const deer_model *model, int B, int T, int op);
+
+/* The same for any forcing, warm-up included, and for the quasi-DEER entry points when
+ * quasi != 0.  With T_w > 0 the solve runs as two chained solves -- the warm-up prefix with
+ * alpha = 1, then the rest from z_0 := P_1 z_{T_w} + zbar_{T_w} -- which have the joint
+ * problem's unique zero (the segments are copied through the workspace), and the adjoint as
+ * the rest's adjoint followed by the prefix's, seeded with J~_{T_w+1}^T lam_{T_w+1}
+ * (diag(J~_{T_w+1}) lam_{T_w+1} for quasi-DEER); the parameter gradients are summed. */
+size_t deer_workspace_bytes_ex(const deer_model *model, const deer_forcing *forcing, int B, int T, int op,
+                               int quasi);
 
 /* GTF-DEER forward solve (Alg. GTF-DEER, Newton loop; eqs. GTF_residual, GTF_DEER_update).
  *   x, z0        inputs as above; z0 may be NULL.

@@ -146,27 +146,27 @@ def _workspace(nbytes: int):
 
 def deer_solve(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1e-5, max_iter: int = 500,
                fixed_iters: int = 0, init: str = "teacher", z=None, want_masks: bool = False, ws=None,
-               check: bool = True, step_bound: float = 0.0) -> dict:
+               check: bool = True, step_bound: float = 0.0, T_w: int = 0) -> dict:
     """GTF-DEER forward solve.  Returns dict(z, masks, iters, norms, status).  step_bound:
     threshold of the update safeguard (0: library default, < 0: only non-finite updates are
-    rejected)."""
-    return _solve("deer_solve", "deer_workspace_bytes", model, x, alpha, n_forced, z0=z0, tol=tol,
-                  max_iter=max_iter, fixed_iters=fixed_iters, init=init, z=z, want_masks=want_masks, ws=ws,
-                  check=check, step_bound=step_bound)
+    rejected).  T_w: latent warm-up steps."""
+    return _solve("deer_solve", 0, model, x, alpha, n_forced, z0=z0, tol=tol, max_iter=max_iter,
+                  fixed_iters=fixed_iters, init=init, z=z, want_masks=want_masks, ws=ws, check=check,
+                  step_bound=step_bound, T_w=T_w)
 
 
 def deer_solve_quasi(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1e-5, max_iter: int = 500,
                      fixed_iters: int = 0, init: str = "teacher", z=None, want_masks: bool = False, ws=None,
-                     check: bool = True, step_bound: float = 0.0) -> dict:
+                     check: bool = True, step_bound: float = 0.0, T_w: int = 0) -> dict:
     """Quasi-DEER forward solve (diagonal Jacobians; PLRNN kinds): arguments and result as
     deer_solve."""
-    return _solve("deer_solve_quasi", "deer_quasi_workspace_bytes", model, x, alpha, n_forced, z0=z0, tol=tol,
-                  max_iter=max_iter, fixed_iters=fixed_iters, init=init, z=z, want_masks=want_masks, ws=ws,
-                  check=check, step_bound=step_bound)
+    return _solve("deer_solve_quasi", 1, model, x, alpha, n_forced, z0=z0, tol=tol, max_iter=max_iter,
+                  fixed_iters=fixed_iters, init=init, z=z, want_masks=want_masks, ws=ws, check=check,
+                  step_bound=step_bound, T_w=T_w)
 
 
-def _solve(entry, ws_entry, model, x, alpha, n_forced, *, z0, tol, max_iter, fixed_iters, init, z, want_masks, ws,
-           check, step_bound):
+def _solve(entry, quasi, model, x, alpha, n_forced, *, z0, tol, max_iter, fixed_iters, init, z, want_masks, ws,
+           check, step_bound, T_w):
     lib = load()
     m = _model(model)
     x = _dev(x)
@@ -182,11 +182,11 @@ def _solve(entry, ws_entry, model, x, alpha, n_forced, *, z0, tol, max_iter, fix
     if want_masks:
         H = m.M if m.kind == "plrnn" else m.L
         masks = torch.empty(B, T, (H + 31) // 32, dtype=torch.int32, device="cuda")
+    f = _b.deer_forcing(float(alpha), int(n_forced), int(T_w))
     if ws is None:
-        ws = _workspace(getattr(lib, ws_entry)(ctypes.byref(m.c), B, T, _b.DEER_OP_SOLVE))
+        ws = _workspace(lib.deer_workspace_bytes_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _b.DEER_OP_SOLVE, quasi))
     iters = (ctypes.c_int32 * B)()
     norms = (ctypes.c_float * B)()
-    f = _b.deer_forcing(float(alpha), int(n_forced))
     o = _b.deer_solve_opts(float(tol), int(max_iter), int(fixed_iters), _INITS[init], float(step_bound))
     z0d = _dev(z0)
     st = getattr(lib, entry)(ctypes.byref(m.c), ctypes.byref(f), ctypes.byref(o), B, T, _ptr(x), _ptr(z0d),
@@ -198,7 +198,7 @@ def _solve(entry, ws_entry, model, x, alpha, n_forced, *, z0, tol, max_iter, fix
 
 
 def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, want_lam: bool = True,
-                 want_grads: bool = True, ws=None) -> dict:
+                 want_grads: bool = True, ws=None, T_w: int = 0) -> dict:
     """Adjoint scan lam = dL/dz and parameter gradients at trajectory z.  Diagonal SSM: g is
     complex [B,T,M] (or [B,T,M,2] float) = dL/dRe h + i dL/dIm h, or a real float tensor
     [B,T,M] = dL/dRe h (the read-out's cotangent)."""
@@ -232,9 +232,9 @@ def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, w
         else:
             grads = {"lam": torch.empty(m.M, 2, device="cuda"), "Bc": torch.empty(m.M, m.L, 2, device="cuda")}
             gs = _b.deer_grads(_ptr(grads["lam"]), _ptr(grads["Bc"]), None, None, None)
+    f = _b.deer_forcing(float(alpha), int(n_forced), int(T_w))
     if ws is None:
-        ws = _workspace(lib.deer_workspace_bytes(ctypes.byref(m.c), B, T, _b.DEER_OP_ADJOINT))
-    f = _b.deer_forcing(float(alpha), int(n_forced))
+        ws = _workspace(lib.deer_workspace_bytes_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _b.DEER_OP_ADJOINT, 0))
     z0d = _dev(z0)
     st = lib.deer_adjoint_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(g),
                              g_layout, _ptr(lam), ctypes.byref(gs), _ptr(ws), ws.numel(), _stream())
@@ -243,7 +243,7 @@ def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, w
 
 
 def deer_adjoint_quasi(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, want_lam: bool = True,
-                       want_grads: bool = True, ws=None) -> dict:
+                       want_grads: bool = True, ws=None, T_w: int = 0) -> dict:
     """Quasi-DEER adjoint (diagonal Jacobians; PLRNN kinds) and parameter gradients at
     trajectory z: arguments and result as deer_adjoint."""
     lib = load()
@@ -257,9 +257,9 @@ def deer_adjoint_quasi(model, x, z, alpha: float, n_forced: int, *, z0=None, g=N
     g = _dev(g)
     lam = torch.empty((B, T, m.M), device="cuda") if want_lam else None
     grads, gs = _plrnn_grads(m) if want_grads else ({}, _b.deer_grads())
+    f = _b.deer_forcing(float(alpha), int(n_forced), int(T_w))
     if ws is None:
-        ws = _workspace(lib.deer_quasi_workspace_bytes(ctypes.byref(m.c), B, T, _b.DEER_OP_ADJOINT))
-    f = _b.deer_forcing(float(alpha), int(n_forced))
+        ws = _workspace(lib.deer_workspace_bytes_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _b.DEER_OP_ADJOINT, 1))
     z0d = _dev(z0)
     st = lib.deer_adjoint_quasi(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(g),
                                 _ptr(lam), ctypes.byref(gs), _ptr(ws), ws.numel(), _stream())

@@ -24,7 +24,8 @@ DEER_G_NATIVE, DEER_G_REAL = 0, 1
 EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "deer_adjoint_ex", "plrnn_jacobian", "deer_scan",
             "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_readout_loss", "deer_status_string",
             "deer_last_error", "deer_timing_enable", "deer_timing_report", "deer_solve_quasi", "deer_adjoint_quasi",
-            "deer_quasi_workspace_bytes", "deer_sequential", "deer_sequential_workspace_bytes"]
+            "deer_quasi_workspace_bytes", "deer_sequential", "deer_sequential_workspace_bytes",
+            "deer_workspace_bytes_ex"]
 
 _fp = ctypes.c_void_p
 
@@ -35,7 +36,7 @@ class deer_model(ctypes.Structure):
 
 
 class deer_forcing(ctypes.Structure):
-    _fields_ = [("alpha", ctypes.c_float), ("n_forced", ctypes.c_int)]
+    _fields_ = [("alpha", ctypes.c_float), ("n_forced", ctypes.c_int), ("T_w", ctypes.c_int)]
 
 
 class deer_solve_opts(ctypes.Structure):
@@ -83,6 +84,8 @@ def load(path: str = LIB_PATH):
     lib.deer_solve_quasi.restype = i32
     lib.deer_adjoint_quasi.argtypes = lib.deer_adjoint.argtypes
     lib.deer_adjoint_quasi.restype = i32
+    lib.deer_workspace_bytes_ex.argtypes = [P(deer_model), P(deer_forcing), i32, i32, i32, i32]
+    lib.deer_workspace_bytes_ex.restype = sz
     lib.deer_quasi_workspace_bytes.argtypes = [P(deer_model), i32, i32, i32]
     lib.deer_quasi_workspace_bytes.restype = sz
     lib.deer_adjoint_ex.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, i32, vp, P(deer_grads),

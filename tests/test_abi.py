@@ -88,3 +88,28 @@ def test_argument_errors_before_device_work(lib):
 def test_status_strings(lib):
     for code in range(6):
         assert lib.deer_status_string(code)
+
+
+def test_warmup_arguments(lib):
+    m, _keep = _vanilla_model(4)
+    o = _b.deer_solve_opts(1e-5, 10, 0, 0, 0.0)
+    base = lib.deer_workspace_bytes(ctypes.byref(m), 2, 64, _b.DEER_OP_SOLVE)
+    f0 = _b.deer_forcing(0.1, 2, 0)
+    assert lib.deer_workspace_bytes_ex(ctypes.byref(m), ctypes.byref(f0), 2, 64, _b.DEER_OP_SOLVE, 0) == base
+    fw = _b.deer_forcing(0.1, 2, 16)
+    for op in (_b.DEER_OP_SOLVE, _b.DEER_OP_ADJOINT):
+        for q in (0, 1):
+            assert lib.deer_workspace_bytes_ex(ctypes.byref(m), ctypes.byref(fw), 2, 64, op, q) > 0
+    bad = _b.deer_forcing(0.1, 2, 64)                  # T_w must be < T
+    assert lib.deer_workspace_bytes_ex(ctypes.byref(m), ctypes.byref(bad), 2, 64, _b.DEER_OP_SOLVE, 0) == 0
+    st = lib.deer_solve(ctypes.byref(m), ctypes.byref(bad), ctypes.byref(o), 2, 64, None, None, None, None,
+                        None, None, None, 0, None)
+    assert st == _b.DEER_ERR_INVALID_ARG and b"T_w" in lib.deer_last_error()
+    fixed = _b.deer_solve_opts(1e-5, 10, 3, 0, 0.0)     # warm-up needs a tolerance solve
+    dummy = (ctypes.c_float * 16)()
+    p = ctypes.cast(dummy, ctypes.c_void_p)
+    st = lib.deer_solve(ctypes.byref(m), ctypes.byref(fw), ctypes.byref(fixed), 2, 64, p, None, p, None,
+                        None, None, None, 0, None)
+    assert st == _b.DEER_ERR_INVALID_ARG and b"tolerance" in lib.deer_last_error()
+    dg = _b.deer_model(_b.DEER_DIAG_SSM, 4, 3, m.A, m.W, None, None, None)
+    assert lib.deer_workspace_bytes_ex(ctypes.byref(dg), ctypes.byref(fw), 2, 64, _b.DEER_OP_SOLVE, 0) == 0

@@ -536,3 +536,62 @@ def diag_ssm_step(params: dict, x: np.ndarray) -> dict:
     grads = diag_ssm_param_grads(a_adj, h, x)
     grads.update(mlp_grads)
     return {"b": b, "h": h, "loss": loss, "g": g, "a": a_adj, "grads": grads}
+
+
+# --------------------------------------------------------------------------------------
+# training step around the gradient: MAR penalty and the parameter update
+# --------------------------------------------------------------------------------------
+
+def mar_loss_and_grads(model: dict, M_r: int, lam_mar: float, p: int, gamma_w: float, gamma_v: float):
+    """Manifold attractor regularisation on the last M_r latents (eq. mar_loss_latent_initscale):
+    lam_mar / M_r * sum_i [ |1 - A_i|^p + (1/L) sum_j (gamma_w |W_ij|^p + gamma_v |V_ji|^p) + |h_i|^p ].
+    Vanilla PLRNN: V = I is not a parameter (no V term) and L = M; shallow: W = W1, V = W2,
+    h = h1.  Returns (loss, grads) with the derivative of |u|^p taken as p |u|^(p-1) sign(u)
+    (0 at u = 0 for p = 1)."""
+    model = _model64(model)
+    A = _p(model, "A")
+    M = A.shape[0]
+    sl = slice(M - M_r, M)
+    c = lam_mar / M_r
+
+    def pen(u):
+        return np.abs(u) ** p
+
+    def dpen(u):
+        return p * np.abs(u) ** (p - 1) * np.sign(u) if p > 1 else np.sign(u)
+
+    vanilla = model["kind"] == "plrnn"
+    W = _p(model, "W") if vanilla else _p(model, "W1")
+    h = _p(model, "h") if vanilla else _p(model, "h1")
+    L = W.shape[1]
+    loss = c * (pen(1.0 - A[sl]).sum() + pen(h[sl]).sum() + gamma_w / L * pen(W[sl]).sum())
+    gA = np.zeros_like(A)
+    gA[sl] = -c * dpen(1.0 - A[sl])
+    gW = np.zeros_like(W)
+    gW[sl] = c * gamma_w / L * dpen(W[sl])
+    gh = np.zeros_like(h)
+    gh[sl] = c * dpen(h[sl])
+    if vanilla:
+        return float(loss), {"A": gA, "W": gW, "h": gh}
+    V = _p(model, "W2")
+    loss += c * gamma_v / L * pen(V[:, sl]).sum()
+    gV = np.zeros_like(V)
+    gV[:, sl] = c * gamma_v / L * dpen(V[:, sl])
+    return float(loss), {"A": gA, "W1": gW, "W2": gV, "h1": gh, "h2": np.zeros(L)}
+
+
+def adam_update(params: dict, grads: dict, state: dict, step: int, lr: float, beta1: float = 0.9,
+                beta2: float = 0.999, eps: float = 1e-8):
+    """One Adam step (Kingma and Ba): m = b1 m + (1 - b1) g, v = b2 v + (1 - b2) g^2,
+    theta -= lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps), t = step >= 1.  The paper
+    names no optimiser; this is the reading taken.  Returns (new params, new state)."""
+    out, st = {}, {}
+    for k, g in grads.items():
+        g = np.asarray(g, f64)
+        m = beta1 * state.get(("m", k), np.zeros_like(g)) + (1 - beta1) * g
+        v = beta2 * state.get(("v", k), np.zeros_like(g)) + (1 - beta2) * g * g
+        mh = m / (1 - beta1 ** step)
+        vh = v / (1 - beta2 ** step)
+        out[k] = np.asarray(params[k], f64) - lr * mh / (np.sqrt(vh) + eps)
+        st[("m", k)], st[("v", k)] = m, v
+    return out, st

@@ -664,3 +664,46 @@ def test_warmup_as_two_chained_solves(kind):
     g_b = O.param_grads(m, x2, z2, alpha, N, lam2, z0=zb)
     for k in gr:
         assert np.allclose(g_a[k] + g_b[k], gr[k], rtol=1e-11, atol=1e-14), k
+
+
+# ------------------------------------------------------------------------------------
+# training step: MAR penalty (eq. mar_loss_latent_initscale) and the Adam update
+# ------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("kind,p", [("plrnn", 1), ("plrnn", 2), ("shplrnn", 1), ("shplrnn", 2)])
+def test_mar_penalty_matches_autograd(kind, p):
+    M, M_r = 6, 3
+    m = _vanilla(M, 81) if kind == "plrnn" else _shallow(M, 5, 82)
+    lam_mar, gw, gv = 0.7, 0.3, 0.2
+    loss, gr = O.mar_loss_and_grads(m, M_r, lam_mar, p, gw, gv)
+    P = {k: torch.tensor(np.asarray(v, np.float64), requires_grad=True) for k, v in m.items() if k != "kind"}
+    W = P["W"] if kind == "plrnn" else P["W1"]
+    h = P["h"] if kind == "plrnn" else P["h1"]
+    L = W.shape[1]
+    tl = (torch.abs(1 - P["A"][M - M_r:]) ** p).sum() + (torch.abs(h[M - M_r:]) ** p).sum() \
+        + gw / L * (torch.abs(W[M - M_r:]) ** p).sum()
+    if kind == "shplrnn":
+        tl = tl + gv / L * (torch.abs(P["W2"][:, M - M_r:]) ** p).sum()
+    tl = lam_mar / M_r * tl
+    tl.backward()
+    assert abs(loss - float(tl)) < 1e-13
+    for k, v in P.items():
+        ref = v.grad.numpy() if v.grad is not None else np.zeros(v.shape)
+        assert np.allclose(gr[k], ref, rtol=1e-12, atol=1e-15), k
+
+
+def test_adam_matches_torch_adam():
+    rng = np.random.default_rng(83)
+    params = {"a": rng.standard_normal(7), "b": rng.standard_normal((3, 4))}
+    tp = {k: torch.tensor(v.copy(), requires_grad=True) for k, v in params.items()}
+    opt = torch.optim.Adam(list(tp.values()), lr=1e-2, betas=(0.9, 0.99), eps=1e-6)
+    state = {}
+    for step in range(1, 4):
+        grads = {k: rng.standard_normal(v.shape) for k, v in params.items()}
+        params, state = O.adam_update(params, grads, state, step, 1e-2, 0.9, 0.99, 1e-6)
+        opt.zero_grad()
+        for k, v in tp.items():
+            v.grad = torch.tensor(grads[k])
+        opt.step()
+        for k in params:
+            assert np.allclose(params[k], tp[k].detach().numpy(), rtol=1e-12, atol=1e-14), (step, k)

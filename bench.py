@@ -57,6 +57,16 @@ def _quasi_step(D, model, xd, c, ws_s, ws_a):
     return sum(res["iters"])
 
 
+def _train_step(D, model, xd, c, ws, st, T_w):
+    # one optimiser step: solve, MSE + MAR loss, gradient, Adam on the parameters in place
+    st["step"] += 1
+    out = D.deer_train_step(model, xd, c.alpha, c.n_obs, step=st["step"], state=st.get("adam"), lr=1e-4,
+                            mar_lambda=1.0, mar_units=max(1, c.M // 4), mar_p=2, mar_gamma_w=1.0 / (3 * c.M),
+                            mar_gamma_v=1.0 / (3 * c.M), T_w=T_w, tol=c.tol, max_iter=c.max_iter, ws=ws)
+    st["adam"] = out["state"]
+    return sum(out["iters"])
+
+
 def _diag_step(D, model, readout, xd, c, ws_s, ws_r, ws_a, bufs):
     res = D.deer_solve(model, xd, 0.0, 0, ws=ws_s, z=bufs["h"])
     r = D.deer_readout_loss(readout, res["z"], xd, g=bufs["g"], ws=ws_r)
@@ -287,6 +297,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--tw", type=int, default=0,
                     help="PLRNN workloads with a tolerance: latent warm-up of this many steps")
+    ap.add_argument("--train", action="store_true",
+                    help="PLRNN workloads with a tolerance: the whole training step (deer_train_step: loss with "
+                         "MAR, gradient, Adam update in place)")
     ap.add_argument("--quasi", action="store_true",
                     help="PLRNN workloads: quasi-DEER (diagonal Jacobians) instead of GTF-DEER")
     ap.add_argument("--fig1a", action="store_true",
@@ -323,7 +336,13 @@ def main():
         step = lambda: _diag_step(D, model, readout, xd, c, ws_s, ws_r, ws_a, bufs)   # noqa: E731
     elif c.kind in ("plrnn", "shplrnn"):
         model = D._Model({"kind": c.kind, **c.params})
-        if args.quasi:
+        if args.train:
+            lib = D.load()
+            fw = Bnd.deer_forcing(float(c.alpha), int(c.n_obs), int(args.tw))
+            ws_t = D._workspace(lib.deer_train_workspace_bytes(ctypes.byref(model.c), ctypes.byref(fw), c.B, c.T, 0))
+            tstate = {"step": 0}
+            step = lambda: _train_step(D, model, xd, c, ws_t, tstate, args.tw)   # noqa: E731
+        elif args.quasi:
             if c.kind != "plrnn":
                 print("quasi-DEER is built for the vanilla PLRNN workloads (1, 2, 5)", file=sys.stderr)
                 sys.exit(3)
@@ -397,7 +416,8 @@ def main():
         "config": {"workload": c.name, "kind": c.kind, "B": c.B, "T": c.T, "M": c.M, "N": c.n_obs,
                    "alpha": c.alpha, "tol": c.tol if not c.fixed_iters else None,
                    "fixed_iters": c.fixed_iters or None, "newton_updates_per_step": iters_per_step,
-                   "step": ("deer_solve_quasi + deer_adjoint_quasi (quasi-DEER: diagonal Jacobians)" if args.quasi
+                   "step": ("deer_train_step (solve, MSE + MAR loss, gradient, Adam)" if args.train else
+                            "deer_solve_quasi + deer_adjoint_quasi (quasi-DEER: diagonal Jacobians)" if args.quasi
                             else "deer_solve + deer_adjoint"), "latent_warmup": args.tw},
         "roofline": roof,
         "kernels": kernels,

@@ -200,6 +200,41 @@ int deer_adjoint_quasi(const deer_model *model, const deer_forcing *forcing, int
                        float *lam, const deer_grads *grads, void *ws, size_t ws_bytes, void *stream);
 size_t deer_quasi_workspace_bytes(const deer_model *model, int B, int T, int op);
 
+/* Hyper-parameters of deer_train_step. */
+typedef struct {
+    float lr, beta1, beta2, eps;   /* Adam (the paper names no optimiser; Adam is the reading)   */
+    int step;                      /* Adam step t >= 1 (bias corrections 1 - beta^t)             */
+    float mar_lambda;              /* MAR weight lambda_MAR (0: no MAR term)                      */
+    int mar_units;                 /* M_r: MAR acts on the last M_r latents, 1 <= M_r <= M       */
+    int mar_p;                     /* 1 or 2: |.| or squared penalty                             */
+    float mar_gamma_w, mar_gamma_v;/* scales of the W and V terms (the paper: 1/(3L), 1/(3M))    */
+    int quasi;                     /* quasi-DEER solve and adjoint instead of GTF-DEER           */
+} deer_train_opts;
+
+/* One training step of GTF-DEER (Alg. GTF-DEER, the body of its outer loop), PLRNN kinds:
+ *   the solve to opts->tol (deer_solve, or deer_solve_quasi), the loss
+ *     L = MSE(x_{T_w+1:T}, B z_{T_w+1:T}) + L_MAR (eqs. mse_loss_warmup, mar_loss_latent_initscale;
+ *     L_MAR = lambda/M_r sum_{i > M - M_r} [|1 - A_i|^p + (1/L) sum_j (gamma_W |W_ij|^p
+ *     + gamma_V |V_ji|^p) + |h_i|^p], V = W2 and W = W1 for the shallow model, no V term and
+ *     L = M for the vanilla one),
+ *   its gradient (deer_adjoint with the MSE seed, plus the MAR gradient), and one Adam step
+ *   applied IN PLACE to the parameter arrays the model points at (A, W, W2, h, h2; a NULL h or
+ *   h2 stays NULL and untrained).
+ *   z          [B,T,M] out: the solved trajectory (the iterate the gradient is taken at).
+ *   adam_m/v   [P] device, in/out: Adam moments in the layout A | W | h (vanilla) or
+ *              A | W1 | W2 | h1 | h2 (shallow), P = deer_train_params(model); zero before step 1.
+ *   grads      optional outputs of the total gradient (MSE + MAR) before the update, or NULL.
+ *   loss       device [1] out or NULL;  iters host [B] out or NULL.
+ * If the solve does not converge (or is non-finite) its status is returned and the
+ * parameters are left unchanged.  Workspace: deer_train_workspace_bytes(model, forcing, B, T,
+ * train->quasi). */
+int deer_train_step(const deer_model *model, const deer_forcing *forcing, const deer_solve_opts *opts,
+                    const deer_train_opts *train, int B, int T, const float *x, const float *z0, float *z,
+                    float *adam_m, float *adam_v, const deer_grads *grads, float *loss, int32_t *iters,
+                    void *ws, size_t ws_bytes, void *stream);
+size_t deer_train_workspace_bytes(const deer_model *model, const deer_forcing *forcing, int B, int T, int quasi);
+size_t deer_train_params(const deer_model *model);
+
 /* Sequential GTF baseline (the comparison of Fig. 1A): the forward rollout
  *   z_s = F(z~_s), z~ the forced state of eq. GTF, step by step in time,
  * and, when lam or grads is given, back-propagation through time, also step by step:

@@ -21,7 +21,7 @@ from ._binding import DeerError, load  # noqa: F401
 
 __all__ = ["deer_solve", "deer_adjoint", "deer_readout_loss", "plrnn_jacobian", "deer_scan", "deer_workspace_bytes",
            "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_status_string", "DeerError", "load",
-           "deer_sequential", "deer_sequential_workspace_bytes", "deer_solve_quasi", "deer_adjoint_quasi"]
+           "deer_sequential", "deer_sequential_workspace_bytes", "deer_solve_quasi", "deer_adjoint_quasi", "deer_train_step"]
 
 _KINDS = {"plrnn": _b.DEER_PLRNN, "shplrnn": _b.DEER_SHPLRNN, "diag_ssm": _b.DEER_DIAG_SSM}
 _INITS = {"teacher": _b.DEER_INIT_TEACHER, "zero": _b.DEER_INIT_ZERO, "user": _b.DEER_INIT_USER}
@@ -265,6 +265,44 @@ def deer_adjoint_quasi(model, x, z, alpha: float, n_forced: int, *, z0=None, g=N
                                 _ptr(lam), ctypes.byref(gs), _ptr(ws), ws.numel(), _stream())
     _b._check(st, "deer_adjoint_quasi")
     return {"lam": lam, "grads": grads}
+
+
+def deer_train_step(model, x, alpha: float, n_forced: int, *, step: int, state=None, lr: float = 1e-3,
+                    beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8, mar_lambda: float = 0.0,
+                    mar_units: int = 0, mar_p: int = 2, mar_gamma_w: float = 0.0, mar_gamma_v: float = 0.0,
+                    quasi: bool = False, T_w: int = 0, tol: float = 1e-5, max_iter: int = 500, z0=None,
+                    want_grads: bool = False, ws=None) -> dict:
+    """One GTF-DEER training step (solve, MSE + MAR loss, gradient, Adam) through the C ABI.
+    `model` must be a _Model (its device parameter tensors are updated in place); `state`
+    holds the Adam moments {"m", "v"} (created as zeros when None).  Returns dict(loss, z,
+    iters, grads, state, status)."""
+    lib = load()
+    if not isinstance(model, _Model):
+        raise TypeError("deer_train_step updates the parameters in place: pass a _Model")
+    m = model
+    x = _dev(x)
+    B, T1, _ = x.shape
+    T = T1 - 1
+    P = int(lib.deer_train_params(ctypes.byref(m.c)))
+    if state is None:
+        state = {"m": torch.zeros(P, device="cuda"), "v": torch.zeros(P, device="cuda")}
+    f = _b.deer_forcing(float(alpha), int(n_forced), int(T_w))
+    o = _b.deer_solve_opts(float(tol), int(max_iter), 0, _INITS["teacher"], 0.0)
+    tr = _b.deer_train_opts(float(lr), float(beta1), float(beta2), float(eps), int(step), float(mar_lambda),
+                            int(mar_units), int(mar_p), float(mar_gamma_w), float(mar_gamma_v), int(bool(quasi)))
+    if ws is None:
+        ws = _workspace(lib.deer_train_workspace_bytes(ctypes.byref(m.c), ctypes.byref(f), B, T, int(bool(quasi))))
+    z = torch.empty(B, T, m.M, device="cuda")
+    loss = torch.empty(1, device="cuda")
+    iters = (ctypes.c_int32 * B)()
+    grads, gs = _plrnn_grads(m) if want_grads else ({}, None)
+    z0d = _dev(z0)
+    st = lib.deer_train_step(ctypes.byref(m.c), ctypes.byref(f), ctypes.byref(o), ctypes.byref(tr), B, T, _ptr(x),
+                             _ptr(z0d), _ptr(z), _ptr(state["m"]), _ptr(state["v"]),
+                             ctypes.byref(gs) if gs is not None else None, _ptr(loss), iters, _ptr(ws), ws.numel(),
+                             _stream())
+    _b._check(st, "deer_train_step")
+    return {"loss": loss, "z": z, "iters": list(iters), "grads": grads, "state": state, "status": st}
 
 
 def _plrnn_grads(m):

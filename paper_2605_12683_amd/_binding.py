@@ -25,7 +25,7 @@ EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "deer_adjoint_
             "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_readout_loss", "deer_status_string",
             "deer_last_error", "deer_timing_enable", "deer_timing_report", "deer_solve_quasi", "deer_adjoint_quasi",
             "deer_quasi_workspace_bytes", "deer_sequential", "deer_sequential_workspace_bytes",
-            "deer_workspace_bytes_ex"]
+            "deer_workspace_bytes_ex", "deer_train_step", "deer_train_workspace_bytes", "deer_train_params"]
 
 _fp = ctypes.c_void_p
 
@@ -33,6 +33,13 @@ _fp = ctypes.c_void_p
 class deer_model(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int), ("M", ctypes.c_int), ("L", ctypes.c_int),
                 ("A", _fp), ("W", _fp), ("W2", _fp), ("h", _fp), ("h2", _fp)]
+
+
+class deer_train_opts(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("step", ctypes.c_int), ("mar_lambda", ctypes.c_float), ("mar_units", ctypes.c_int),
+                ("mar_p", ctypes.c_int), ("mar_gamma_w", ctypes.c_float), ("mar_gamma_v", ctypes.c_float),
+                ("quasi", ctypes.c_int)]
 
 
 class deer_forcing(ctypes.Structure):
@@ -84,6 +91,13 @@ def load(path: str = LIB_PATH):
     lib.deer_solve_quasi.restype = i32
     lib.deer_adjoint_quasi.argtypes = lib.deer_adjoint.argtypes
     lib.deer_adjoint_quasi.restype = i32
+    lib.deer_train_step.argtypes = [P(deer_model), P(deer_forcing), P(deer_solve_opts), P(deer_train_opts), i32, i32,
+                                    vp, vp, vp, vp, vp, P(deer_grads), vp, P(ctypes.c_int32), vp, sz, vp]
+    lib.deer_train_step.restype = i32
+    lib.deer_train_workspace_bytes.argtypes = [P(deer_model), P(deer_forcing), i32, i32, i32]
+    lib.deer_train_workspace_bytes.restype = sz
+    lib.deer_train_params.argtypes = [P(deer_model)]
+    lib.deer_train_params.restype = sz
     lib.deer_workspace_bytes_ex.argtypes = [P(deer_model), P(deer_forcing), i32, i32, i32, i32]
     lib.deer_workspace_bytes_ex.restype = sz
     lib.deer_quasi_workspace_bytes.argtypes = [P(deer_model), i32, i32, i32]

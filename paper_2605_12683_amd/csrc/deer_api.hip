@@ -1373,6 +1373,95 @@ size_t deer_workspace_bytes_ex(const deer_model *m, const deer_forcing *f, int B
     return bytes;
 }
 
+size_t deer_train_params(const deer_model *m) {
+    if (!m || (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN)) return 0;
+    return param_floats(m);
+}
+
+size_t deer_train_workspace_bytes(const deer_model *m, const deer_forcing *f, int B, int T, int quasi) {
+    const size_t a = deer_workspace_bytes_ex(m, f, B, T, DEER_OP_SOLVE, quasi);
+    const size_t b = deer_workspace_bytes_ex(m, f, B, T, DEER_OP_ADJOINT, quasi);
+    if (!a || !b || (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN)) return 0;
+    Carver c(nullptr);
+    c.take<float>(param_floats(m));
+    c.take<double>(train_partials() + 1);
+    c.take<char>(a > b ? a : b);
+    return c.off;
+}
+
+int deer_train_step(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, const deer_train_opts *tr,
+                    int B, int T, const float *x, const float *z0, float *z, float *adam_m, float *adam_v,
+                    const deer_grads *grads_out, float *loss, int32_t *iters, void *ws, size_t ws_bytes,
+                    void *stream) {
+    set_error("");
+    int rc = check_common(m, f, B, T);
+    if (rc) return rc;
+    if (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN) { set_error("deer_train_step: PLRNN kinds only"); return DEER_ERR_INVALID_ARG; }
+    if (!o || !tr || !x || !z || !adam_m || !adam_v) { set_error("opts, train, x, z and the Adam moments are required"); return DEER_ERR_INVALID_ARG; }
+    if (o->fixed_iters > 0) { set_error("deer_train_step solves to a tolerance (fixed_iters = 0)"); return DEER_ERR_INVALID_ARG; }
+    if (tr->step < 1 || !(tr->lr > 0.f) || !(tr->beta1 >= 0.f && tr->beta1 < 1.f) || !(tr->beta2 >= 0.f && tr->beta2 < 1.f)) {
+        set_error("Adam needs step >= 1, lr > 0 and betas in [0, 1)");
+        return DEER_ERR_INVALID_ARG;
+    }
+    if (tr->mar_lambda != 0.f && (tr->mar_units < 1 || tr->mar_units > m->M || (tr->mar_p != 1 && tr->mar_p != 2))) {
+        set_error("MAR needs 1 <= mar_units <= M and mar_p in {1, 2}");
+        return DEER_ERR_INVALID_ARG;
+    }
+    if (f->n_forced < 1) { set_error("the MSE needs at least one observed latent (n_forced >= 1)"); return DEER_ERR_INVALID_ARG; }
+    const bool quasi = tr->quasi != 0;
+    const size_t need = deer_train_workspace_bytes(m, f, B, T, tr->quasi);
+    if ((rc = check_ws(ws, ws_bytes, need))) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    Carver c(ws);
+    float *g = c.take<float>(param_floats(m));
+    double *part = c.take<double>(train_partials() + 1);
+    const size_t a = deer_workspace_bytes_ex(m, f, B, T, DEER_OP_SOLVE, tr->quasi);
+    const size_t b = deer_workspace_bytes_ex(m, f, B, T, DEER_OP_ADJOINT, tr->quasi);
+    const size_t inner_bytes = a > b ? a : b;
+    void *inner = c.take<char>(inner_bytes);
+    // the solve, then the gradient of the MSE at its result (the adjoint's own MSE seed)
+    rc = (quasi ? deer_solve_quasi : deer_solve)(m, f, o, B, T, x, z0, z, nullptr, iters, nullptr, inner, inner_bytes,
+                                                 stream);
+    if (rc) return rc;
+    const deer_grads gbuf = grads_at(m, g);
+    rc = (quasi ? deer_adjoint_quasi : deer_adjoint)(m, f, B, T, x, z0, z, nullptr, nullptr, &gbuf, inner,
+                                                     inner_bytes, stream);
+    if (rc) return rc;
+    if (!m->h) {   // untrained (absent) biases: zero gradients so the layout stays uniform
+        if ((rc = launch_fill_f32(gbuf.h, m->M, 0.f, st))) return rc;
+    }
+    if (m->kind == DEER_SHPLRNN && !m->h2) {
+        if ((rc = launch_fill_f32(gbuf.h2, m->L, 0.f, st))) return rc;
+    }
+    const bool sh = m->kind == DEER_SHPLRNN;
+    double *mar = part + train_partials();
+    const bool with_mar = tr->mar_lambda != 0.f;
+    if (with_mar && (rc = launch_mar(sh, m->A, m->W, sh ? m->W2 : nullptr, m->h, m->M, sh ? m->L : m->M,
+                                     tr->mar_units, tr->mar_lambda, tr->mar_p, tr->mar_gamma_w, tr->mar_gamma_v, g,
+                                     mar, st)))
+        return rc;
+    if (loss) {
+        if ((rc = launch_mse_loss_partial(z, x, B, T, m->M, f->n_forced, f->T_w, part, st))) return rc;
+        const double scale = 1.0 / ((double)B * f->n_forced * (T - f->T_w));
+        if ((rc = launch_loss_final(part, scale, with_mar ? mar : nullptr, loss, st))) return rc;
+    }
+    if (grads_out) {
+        const size_t M = m->M, L = m->L;
+        const float *src[5] = {gbuf.A, gbuf.W, gbuf.W2, gbuf.h, gbuf.h2};
+        float *dst[5] = {grads_out->A, grads_out->W, sh ? grads_out->W2 : nullptr, grads_out->h,
+                         sh ? grads_out->h2 : nullptr};
+        const size_t n[5] = {M, sh ? M * L : M * M, L * M, M, L};
+        for (int k = 0; k < 5; ++k)
+            if (dst[k]) DEER_HIP(hipMemcpyAsync(dst[k], src[k], n[k] * sizeof(float), hipMemcpyDeviceToDevice, st));
+    }
+    // Adam on the parameters in place
+    const long M = m->M, L = m->L;
+    float *params[5] = {const_cast<float *>(m->A), const_cast<float *>(m->W), sh ? const_cast<float *>(m->W2) : nullptr,
+                        const_cast<float *>(m->h), sh ? const_cast<float *>(m->h2) : nullptr};
+    const long sizes[5] = {M, sh ? M * L : M * M, sh ? L * M : 0, M, sh ? L : 0};
+    return launch_adam(params, sizes, g, adam_m, adam_v, tr->lr, tr->beta1, tr->beta2, tr->eps, tr->step, st);
+}
+
 size_t deer_quasi_workspace_bytes(const deer_model *m, int B, int T, int op) {
     deer_forcing f{0.f, 0};
     if (check_quasi(m, &f, B, T) != DEER_OK) return 0;

@@ -108,6 +108,16 @@ size_t reduce_gpart_ws_bytes(int MP);
 bool newton_small_fits(int M, int T, int fixed_iters);
 int launch_newton_small(const PlrnnArgs &a, float *z, int iters, uint32_t *norm_bits, hipStream_t st);
 
+// training step: MSE partial sums (t > T_w), MAR loss and gradient, the loss, one Adam step
+size_t train_partials();
+int launch_mse_loss_partial(const float *z, const float *x, int B, int T, int M, int N, int T_w, double *part,
+                            hipStream_t st);
+int launch_mar(bool shallow, const float *A, const float *W, const float *V, const float *h, int M, int L, int M_r,
+               float lam, int p, float gw, float gv, float *g, double *mar, hipStream_t st);
+int launch_loss_final(const double *part, double scale, const double *mar, float *loss, hipStream_t st);
+int launch_adam(float *const *params, const long *sizes, const float *g, float *m, float *v, float lr, float b1,
+                float b2, float eps, int step, hipStream_t st);
+
 // quasi-DEER, vanilla PLRNN (diagonal Jacobians): chunk length, one forward Newton update
 // (r and gamma d at the current iterate, chunked diagonal scan, z + Delta to the other buffer,
 // per-chain maxima), and the quasi adjoint with per-chain gradient partials

@@ -276,7 +276,8 @@ static int group_maps_override() {
     return e ? atoi(e) : -1;
 }
 
-// DEER_SMALL=0 keeps small fixed-update solves on the general path (a test override)
+// DEER_SMALL=0 keeps small fixed-update solves and small adjoints on the general path (a test
+// override)
 static bool small_path_enabled() {
     const char *e = getenv("DEER_SMALL");
     return !e || atoi(e) != 0;
@@ -1259,6 +1260,15 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
         PlrnnWs w = carve_plrnn(ws, B, T, m->M, DEER_OP_ADJOINT, &need);
         PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
         const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
+        if (small_path_enabled() && adjoint_small_fits(m->M, T)) {   // one workgroup per sequence
+            const bool gr = grads && (grads->A || grads->W || grads->h);
+            if (B == 1)
+                return launch_adjoint_small(a, g, scale, z, lam, nullptr, gr ? grads->A : nullptr,
+                                            gr ? grads->W : nullptr, gr ? grads->h : nullptr, st);
+            if ((rc = launch_adjoint_small(a, g, scale, z, lam, w.gpart, nullptr, nullptr, nullptr, st))) return rc;
+            if (gr) return launch_reduce_gpart(w.gpart, B, 4, m->M, grads->A, grads->W, grads->h, w.gpart2, st);
+            return DEER_OK;
+        }
         if (w.MP == 16) {   // register-tiled path: masks from z inside the kernels, per-wave gradients
             if ((rc = launch_adjoint_plrnn16(a, g, scale, z, w.P, w.v, w.carry, lam, w.gpart, w.C, w.ncs, st)))
                 return rc;

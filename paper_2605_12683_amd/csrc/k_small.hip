@@ -264,6 +264,263 @@ __global__ __launch_bounds__(SNT) void k_newton_small(const float *__restrict__ 
     }
 }
 
+// The adjoint of the same small problems in one launch (gradients appendix: lam_{s} =
+// J~_{s+1}^T lam_{s+1} + g_s from the end, eq. backward_recursion): every thread takes an
+// 8-step chunk, forms the map of its chunk in reverse (the product of the transposed
+// Jacobians and the local adjoint from a zero carry), the carries run over the chunks from
+// the last one in two levels through LDS, and each chunk is re-walked from its carry with the
+// adjoint (optionally) written and the parameter-gradient partial sums of the thread,
+//   dW_ij += lam_i relu(z~_j), dA_i += lam_i z~_i, dh_i += lam_i,
+// summed over the workgroup into gpart[b][SMS][SMS + 2] for the float64 reduction over the batch.
+__global__ __launch_bounds__(SNT) void k_adjoint_small(const float *__restrict__ A, const float *__restrict__ W,
+                                                       float alpha, int N, const float *__restrict__ x,
+                                                       const float *__restrict__ z0, const float *__restrict__ z,
+                                                       const float *__restrict__ g, float seed_scale, int T, int M,
+                                                       int nc, float *__restrict__ lam, float *__restrict__ gpart,
+                                                       float *__restrict__ dA, float *__restrict__ dW,
+                                                       float *__restrict__ dh) {
+    __shared__ float Pm[SNT][SPV];
+    __shared__ float Gm[SNG][SPV];
+    __shared__ float Xg[SNG][SMS];
+    __shared__ float Xc[SNT][SMS];
+    __shared__ float red[SNT / 64][SMS * (SMS + 2)];
+    const int b = blockIdx.x, c = threadIdx.x;
+    float Ai[SMS], pj[SMS], Wm[SMS][SMS];
+#pragma unroll
+    for (int i = 0; i < SMS; ++i) {
+        Ai[i] = i < M ? A[i] : 0.f;
+        pj[i] = i < N ? __fsub_rn(1.0f, alpha) : 1.0f;
+#pragma unroll
+        for (int j = 0; j < SMS; ++j) Wm[i][j] = (i < M && j < M) ? W[i * M + j] : 0.f;
+    }
+    const float *xb = x + (size_t)b * (T + 1) * N;
+    const float *zb = z + (size_t)b * T * M;
+    const bool act = c < nc;
+    const int s0 = c * SC, s1 = act ? min(s0 + SC, T) : s0;
+    // forced inputs z~_s for s = s0 .. s0 + SC (the last one feeds J~ of the chunk's last step)
+    // and the cotangent rows g_s of the chunk
+    float zt[SC + 1][SMS], gr[SC][SMS];
+#pragma unroll
+    for (int k = 0; k <= SC; ++k) {
+        const int s = s0 + k;
+        const bool ok = act && s < T && (k < SC || s < T);
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) {
+            float v = 0.f;
+            if (ok && i < M) {
+                if (s == 0) v = z0 ? z0[(size_t)b * M + i] : (i < N ? xb[i] : 0.f);
+                else if (i < N) v = __fadd_rn(__fmul_rn(pj[i], zb[(size_t)(s - 1) * M + i]), __fmul_rn(alpha, xb[(size_t)s * N + i]));
+                else v = zb[(size_t)(s - 1) * M + i];
+            }
+            zt[k][i] = v;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < SC; ++k) {
+        const int s = s0 + k;
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) {
+            float v = 0.f;
+            if (s < s1 && i < M) {
+                if (g) v = g[((size_t)b * T + s) * M + i];
+                else if (i < N) v = __fmul_rn(seed_scale, __fsub_rn(zb[(size_t)s * M + i], xb[(size_t)(s + 1) * N + i]));
+            }
+            gr[k][i] = v;
+        }
+    }
+    // y <- J~_{s+1}^T y + g_s, J~_{s+1} = (diag(A) + W diag(m)) P_alpha at z~_{s+1}; J~_T = 0
+    auto step_t = [&](int k, const float *y, float *out) {
+        const bool has = s0 + k + 1 < T;
+        const float *zn = zt[k + 1];
+#pragma unroll
+        for (int j = 0; j < SMS; ++j) {
+            float a = gr[k][j];
+            if (has) {
+                // (J~^T y)_j = p_j (A_j y_j + m_j sum_i W_ij y_i)
+                float wsum = 0.f;
+#pragma unroll
+                for (int i = 0; i < SMS; ++i) wsum = fmaf(Wm[i][j], y[i], wsum);
+                const float t = fmaf(Ai[j], y[j], zn[j] > 0.f ? wsum : 0.f);
+                a = fmaf(pj[j], t, a);
+            }
+            out[j] = a;
+        }
+    };
+    // map P (row-major) and local adjoint v of the chunk: y_{s0} = P y_{s1} + v
+    float P[SMS][SMS], v[SMS];
+#pragma unroll
+    for (int i = 0; i < SMS; ++i) {
+        v[i] = 0.f;
+#pragma unroll
+        for (int j = 0; j < SMS; ++j) P[i][j] = i == j ? 1.f : 0.f;
+    }
+#pragma unroll
+    for (int k = SC - 1; k >= 0; --k) {
+        if (s0 + k >= s1) continue;
+        float vn[SMS];
+        step_t(k, v, vn);
+        // P <- J~^T P: column by column, without the cotangent
+        float Pn[SMS][SMS];
+#pragma unroll
+        for (int col = 0; col < SMS; ++col) {
+            float y[SMS], o[SMS];
+#pragma unroll
+            for (int i = 0; i < SMS; ++i) y[i] = P[i][col];
+            const bool has = s0 + k + 1 < T;
+            const float *zn = zt[k + 1];
+#pragma unroll
+            for (int j = 0; j < SMS; ++j) {
+                float wsum = 0.f;
+#pragma unroll
+                for (int i = 0; i < SMS; ++i) wsum = fmaf(Wm[i][j], y[i], wsum);
+                o[j] = has ? pj[j] * fmaf(Ai[j], y[j], zn[j] > 0.f ? wsum : 0.f) : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < SMS; ++j) Pn[j][col] = o[j];
+        }
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) {
+            v[i] = vn[i];
+#pragma unroll
+            for (int j = 0; j < SMS; ++j) P[i][j] = Pn[i][j];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < SMS; ++i) {
+        Pm[c][SMS * SMS + i] = v[i];
+#pragma unroll
+        for (int j = 0; j < SMS; ++j) Pm[c][i * SMS + j] = P[i][j];
+    }
+    __syncthreads();
+    // carries from the last chunk: X(nc - 1) = 0, X(k - 1) = P_k X(k) + v_k; processing index
+    // l = nc - 1 - k, groups of GC in processing order
+    auto apply = [&](const float *map, float *y) {
+        float t[SMS];
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) {
+            float a = map[SMS * SMS + i];
+#pragma unroll
+            for (int j = 0; j < SMS; ++j) a = fmaf(map[i * SMS + j], y[j], a);
+            t[i] = a;
+        }
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) y[i] = t[i];
+    };
+    const int GC = (nc + SNG - 1) / SNG;
+    if (c < SNG) {
+        float G[SMS][SMS], gv[SMS];
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) {
+            gv[i] = 0.f;
+#pragma unroll
+            for (int j = 0; j < SMS; ++j) G[i][j] = i == j ? 1.f : 0.f;
+        }
+        const int l0 = min(c * GC, nc), l1 = min(l0 + GC, nc);
+        for (int l = l0; l < l1; ++l) {
+            const float *pk = Pm[nc - 1 - l];
+            float Gn[SMS][SMS];
+#pragma unroll
+            for (int i = 0; i < SMS; ++i)
+#pragma unroll
+                for (int j = 0; j < SMS; ++j) {
+                    float q = 0.f;
+#pragma unroll
+                    for (int k = 0; k < SMS; ++k) q = fmaf(pk[i * SMS + k], G[k][j], q);
+                    Gn[i][j] = q;
+                }
+            apply(pk, gv);
+#pragma unroll
+            for (int i = 0; i < SMS; ++i)
+#pragma unroll
+                for (int j = 0; j < SMS; ++j) G[i][j] = Gn[i][j];
+        }
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) {
+            Gm[c][SMS * SMS + i] = gv[i];
+#pragma unroll
+            for (int j = 0; j < SMS; ++j) Gm[c][i * SMS + j] = G[i][j];
+        }
+    }
+    __syncthreads();
+    if (c == 0) {
+        float X[SMS] = {0.f, 0.f, 0.f, 0.f};
+        for (int g2 = 0; g2 < SNG; ++g2) {
+#pragma unroll
+            for (int i = 0; i < SMS; ++i) Xg[g2][i] = X[i];
+            apply(Gm[g2], X);
+        }
+    }
+    __syncthreads();
+    if (c < SNG) {
+        float X[SMS];
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) X[i] = Xg[c][i];
+        const int l0 = min(c * GC, nc), l1 = min(l0 + GC, nc);
+        for (int l = l0; l < l1; ++l) {
+            const int k = nc - 1 - l;
+#pragma unroll
+            for (int i = 0; i < SMS; ++i) Xc[k][i] = X[i];
+            apply(Pm[k], X);
+        }
+    }
+    __syncthreads();
+    // re-walk from the carry with the gradient partials
+    float L[SMS], gw[SMS][SMS + 2];
+#pragma unroll
+    for (int i = 0; i < SMS; ++i) {
+        L[i] = act ? Xc[c][i] : 0.f;
+#pragma unroll
+        for (int j = 0; j < SMS + 2; ++j) gw[i][j] = 0.f;
+    }
+#pragma unroll
+    for (int k = SC - 1; k >= 0; --k) {
+        if (s0 + k >= s1) continue;
+        float Ln[SMS];
+        step_t(k, L, Ln);
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) L[i] = Ln[i];
+        if (lam) {
+#pragma unroll
+            for (int i = 0; i < SMS; ++i)
+                if (i < M) lam[((size_t)b * T + s0 + k) * M + i] = L[i];
+        }
+#pragma unroll
+        for (int i = 0; i < SMS; ++i) {
+#pragma unroll
+            for (int j = 0; j < SMS; ++j) gw[i][j] = fmaf(L[i], zt[k][j] > 0.f ? zt[k][j] : 0.f, gw[i][j]);
+            gw[i][SMS] = fmaf(L[i], zt[k][i], gw[i][SMS]);
+            gw[i][SMS + 1] += L[i];
+        }
+    }
+    // workgroup sum of the partials (waves, then the eight wave sums)
+#pragma unroll
+    for (int i = 0; i < SMS; ++i)
+#pragma unroll
+        for (int j = 0; j < SMS + 2; ++j) {
+            float t = gw[i][j];
+            for (int off = 32; off > 0; off >>= 1) t += __shfl_xor(t, off, 64);
+            if ((c & 63) == 0) red[c >> 6][i * (SMS + 2) + j] = t;
+        }
+    __syncthreads();
+    if (c < SMS * (SMS + 2)) {
+        float t = 0.f;
+#pragma unroll
+        for (int w = 0; w < SNT / 64; ++w) t += red[w][c];
+        if (gpart) gpart[(size_t)b * SMS * (SMS + 2) + c] = t;
+        // a single sequence: the gradients themselves, no reduction over the batch
+        const int i = c / (SMS + 2), j = c % (SMS + 2);
+        if (i < M && (j >= SMS || j < M)) {
+            if (j < SMS) {
+                if (dW) dW[i * M + j] = t;
+            } else if (j == SMS) {
+                if (dA) dA[i] = t;
+            } else if (dh) {
+                dh[i] = t;
+            }
+        }
+    }
+}
+
 bool newton_small_fits(int M, int T, int fixed_iters) { return M <= SMS && T <= SNT * SC && fixed_iters > 0; }
 
 int launch_newton_small(const PlrnnArgs &a, float *z, int iters, uint32_t *norm_bits, hipStream_t st) {
@@ -275,4 +532,18 @@ int launch_newton_small(const PlrnnArgs &a, float *z, int iters, uint32_t *norm_
     return DEER_OK;
 }
 
+}  // namespace deer
+
+namespace deer {
+bool adjoint_small_fits(int M, int T) { return M <= SMS && T <= SNT * SC; }
+
+int launch_adjoint_small(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *lam,
+                         float *gpart, float *dA, float *dW, float *dh, hipStream_t st) {
+    const int nc = (a.T + SC - 1) / SC;
+    KTimer kt("k_adjoint_small", st);
+    hipLaunchKernelGGL(k_adjoint_small, dim3(a.B), dim3(SNT), 0, st, a.A, a.W, a.alpha, a.N, a.x, a.z0, z, g,
+                       seed_scale, a.T, a.M, nc, lam, gpart, dA, dW, dh);
+    DEER_LAUNCH_CHECK("k_adjoint_small");
+    return DEER_OK;
+}
 }  // namespace deer

@@ -107,6 +107,12 @@ size_t reduce_gpart_ws_bytes(int MP);
 // max |Delta| of the last update
 bool newton_small_fits(int M, int T, int fixed_iters);
 int launch_newton_small(const PlrnnArgs &a, float *z, int iters, uint32_t *norm_bits, hipStream_t st);
+// adjoint and gradient partials of M <= 4, T <= 4096 in one launch per batch: gpart[b][4][6]
+// (MP = 4 for launch_reduce_gpart); with gpart null the gradients of the single sequence go to
+// dA / dW / dh directly (B = 1)
+bool adjoint_small_fits(int M, int T);
+int launch_adjoint_small(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *lam,
+                         float *gpart, float *dA, float *dW, float *dh, hipStream_t st);
 
 // training step: MSE partial sums (t > T_w), MAR loss and gradient, the loss, one Adam step
 size_t train_partials();

@@ -277,6 +277,42 @@ def test_adjoint_and_grads(M, N, B, T, alpha, chunk):
         assert rel_inf(out["grads"][k].cpu().numpy(), g_ref[k]) < TOL, k
 
 
+@pytest.mark.parametrize("M,N,B,T", [(1, 1, 1, 1), (2, 1, 3, 17), (3, 3, 1, 1024), (4, 4, 2, 4096),
+                                   (3, 2, 2, 300), (4, 2, 1, 255), (3, 3, 1, 9)])
+@pytest.mark.parametrize("mode", ["seed", "user_g_z0", "grads_only"])
+def test_small_adjoint_in_one_launch(M, N, B, T, mode):
+    """Small models take the adjoint in one workgroup per sequence (chunk maps of the
+    transposed Jacobians, two-level carries from the last chunk, re-walk with the gradient
+    partials): lam and dL/dtheta against the oracle, and against the general path
+    (DEER_SMALL=0); B = 1 writes the gradients without the batch reduction."""
+    alpha = 0.2
+    c = _case(M, N, B, T, alpha, 400 + M + T)
+    m = oracle_model(c)
+    rng = np.random.default_rng(M + T)
+    z0 = rng.standard_normal((B, M)).astype(np.float32) if mode == "user_g_z0" else None
+    z32 = O.rollout(m, c.x, alpha, N, z0=z0).astype(np.float32)
+    g = rng.standard_normal(z32.shape).astype(np.float32) if mode == "user_g_z0" else None
+    want_lam = mode != "grads_only"
+    say("deer_adjoint small one-launch", M, N, B, T, mode)
+    out = D.deer_adjoint(m, c.x, z32, alpha, N, z0=z0, g=g, want_lam=want_lam)
+    lam_ref = O.adjoint(m, c.x, z32, alpha, N, z0=z0, g=g, mask_precision="float32")
+    g_ref = O.param_grads(m, c.x, z32, alpha, N, lam_ref, z0=z0, mask_precision="float32")
+    if want_lam:
+        assert rel_inf(out["lam"].cpu().numpy(), lam_ref) < TOL
+    for k in ("A", "W", "h"):
+        assert rel_inf(out["grads"][k].cpu().numpy(), g_ref[k]) < TOL, k
+    os.environ["DEER_SMALL"] = "0"
+    try:
+        say("deer_adjoint general path", M, N, B, T, mode)
+        gen = D.deer_adjoint(m, c.x, z32, alpha, N, z0=z0, g=g, want_lam=want_lam)
+    finally:
+        os.environ.pop("DEER_SMALL", None)
+    if want_lam:
+        assert rel_inf(out["lam"].cpu().numpy(), gen["lam"].cpu().numpy()) < TOL
+    for k in ("A", "W", "h"):
+        assert rel_inf(out["grads"][k].cpu().numpy(), gen["grads"][k].cpu().numpy()) < TOL, k
+
+
 def test_adjoint_user_cotangent():
     c = _case(16, 3, 2, 300, 0.2, 19)
     m = oracle_model(c)

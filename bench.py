@@ -31,6 +31,9 @@ sys.path.insert(0, HERE)
 
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 PEAK_FP32_MFMA_TFLOPS = 157.3    # MI355X dense fp32 matrix
+# fp32 vector: 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2 (packed fp32) x 2.4 GHz; the
+# kernels are built without the packed instructions, so half of it is the reachable ceiling
+PEAK_FP32_VALU_TFLOPS = 157.3
 
 
 def log(*a):
@@ -105,6 +108,9 @@ def kernel_work(c, steps, updates):
         # M <= 16 with whole blocks of chunks: one kernel per pass (the fix-up of an update and
         # the forward pass of the next); its matrix-core work is the forward pass's
         out["k_newton_pass16"] = ("mfma", fwd * 2.0 * M ** 3)
+        # M <= 4 with a fixed update count: the whole solve in one launch on the vector units
+        # (the same chunk-map composition, 2 M^3 flops per timestep and update)
+        out["k_newton_small"] = ("alu", fwd * 2.0 * M ** 3)
         out["k_chunk_product_plrnn"] = ("mfma", steps * B * (T - 1) * 2.0 * M ** 3)
         out["k_resjac_plrnn"] = ("hbm", adj * (4 * M + 4 * N + 4 * W))
         # quasi-DEER: residual and diagonal (z, x read; r, d written / adjoint: d written),
@@ -177,6 +183,10 @@ def roofline_for(name, c, total_ms, launches, steps, updates):
         ach = w / (total_ms * 1e-3) / 1e12
         base.update({"bound": "mfma", "achieved": ach, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
                      "frac": ach / PEAK_FP32_MFMA_TFLOPS, "work_per_launch": w / launches})
+    elif bound == "alu":
+        ach = w / (total_ms * 1e-3) / 1e12
+        base.update({"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS, "unit": "TFLOP/s",
+                     "frac": ach / PEAK_FP32_VALU_TFLOPS, "work_per_launch": w / launches})
     else:
         ach = w / (total_ms * 1e-3) / 1e9
         base.update({"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",

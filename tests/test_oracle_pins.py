@@ -707,3 +707,67 @@ def test_adam_matches_torch_adam():
         opt.step()
         for k in params:
             assert np.allclose(params[k], tp[k].detach().numpy(), rtol=1e-12, atol=1e-14), (step, k)
+
+
+def _mar_base(kind, M, L):
+    """A model whose MAR penalty is zero term by term: A = 1, every weight and bias 0."""
+    if kind == "plrnn":
+        return {"kind": "plrnn", "A": np.ones(M, np.float32), "W": np.zeros((M, M), np.float32),
+                "h": np.zeros(M, np.float32)}
+    return {"kind": "shplrnn", "A": np.ones(M, np.float32), "W1": np.zeros((M, L), np.float32),
+            "W2": np.zeros((L, M), np.float32), "h1": np.zeros(M, np.float32), "h2": np.zeros(L, np.float32)}
+
+
+@pytest.mark.parametrize("p", [1, 2])
+@pytest.mark.parametrize("kind,M,L", [("plrnn", 7, 7), ("shplrnn", 5, 9)])
+def test_mar_penalty_closed_forms(kind, M, L, p):
+    """eq. mar_loss_latent_initscale term by term, on models with a single non-zero entry:
+    lambda/M_r [ |1 - A_ii|^p + (1/L) sum_j (gamma_W |W_ij|^p + gamma_V |V_ji|^p) + |h_i|^p ]
+    summed over the last M_r latents i only.  The sum runs over the rows of W (M x L) and the
+    columns of V (L x M) that belong to a MAR latent; L is the hidden width (M for the vanilla
+    PLRNN, which has no V).  Every closed form below is written from the equation, not from the
+    oracle; a row/column swap of V, a 1/M instead of 1/L, or a wrong latent range fails one."""
+    M_r, lam, gw, gv = 3, 0.7, 0.3, 0.2
+    mar = list(range(M - M_r, M))
+    free = list(range(M - M_r))
+    c = lam / M_r
+    wkey, hkey = ("W", "h") if kind == "plrnn" else ("W1", "h1")
+
+    def val(m):
+        return O.mar_loss_and_grads(m, M_r, lam, p, gw, gv)[0]
+
+    assert val(_mar_base(kind, M, L)) == 0.0
+    for i in mar + free:
+        inside = i in mar
+        m = _mar_base(kind, M, L)
+        m["A"][i] = np.float32(0.25)            # |1 - A| = 0.75
+        assert np.isclose(val(m), c * 0.75 ** p if inside else 0.0, rtol=1e-15, atol=0)
+        m = _mar_base(kind, M, L)
+        m[hkey][i] = np.float32(-1.5)
+        assert np.isclose(val(m), c * 1.5 ** p if inside else 0.0, rtol=1e-15, atol=0)
+        m = _mar_base(kind, M, L)
+        m[wkey][i, L - 1] = np.float32(-2.0)    # W_ij: row i is the latent
+        assert np.isclose(val(m), c * gw / L * 2.0 ** p if inside else 0.0, rtol=1e-15, atol=0)
+    if kind == "shplrnn":
+        for i in mar + free:
+            m = _mar_base(kind, M, L)
+            m["W2"][L - 2, i] = np.float32(1.25)  # V_ji: column i is the latent
+            assert np.isclose(val(m), c * gv / L * 1.25 ** p if i in mar else 0.0, rtol=1e-15, atol=0)
+        # V_ij instead of V_ji: a row index that equals a MAR latent index, in a free column
+        m = _mar_base(kind, M, L)
+        m["W2"][mar[0], free[0]] = np.float32(1.25)
+        assert val(m) == 0.0
+    # hidden biases h2 never enter the penalty
+    if kind == "shplrnn":
+        m = _mar_base(kind, M, L)
+        m["h2"][:] = 3.0
+        assert val(m) == 0.0
+    # the terms add: all four at once in one MAR latent
+    i = mar[-1]
+    m = _mar_base(kind, M, L)
+    m["A"][i], m[hkey][i], m[wkey][i, 0] = np.float32(0.5), np.float32(0.5), np.float32(0.5)
+    ref = c * (0.5 ** p + 0.5 ** p + gw / L * 0.5 ** p)
+    if kind == "shplrnn":
+        m["W2"][0, i] = np.float32(0.5)
+        ref += c * gv / L * 0.5 ** p
+    assert np.isclose(val(m), ref, rtol=1e-15, atol=0)

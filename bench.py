@@ -13,7 +13,10 @@ One step = one pass of the whole path over one batch of synthetic input:
 Inputs are resident in HBM before the timed region.  The value is DEER timesteps per
 second: sum over sequences of T x Newton updates, per second of the whole step.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 5]
+
+The default workload is the largest one, the M = 64 vanilla PLRNN (B = 32, T = 131072), whose
+dense 64 x 64 chunk products are the matrix-core bound part of the path.
 """
 from __future__ import annotations
 
@@ -31,9 +34,13 @@ sys.path.insert(0, HERE)
 
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 PEAK_FP32_MFMA_TFLOPS = 157.3    # MI355X dense fp32 matrix
-# fp32 vector: 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2 (packed fp32) x 2.4 GHz; the
-# kernels are built without the packed instructions, so half of it is the reachable ceiling
-PEAK_FP32_VALU_TFLOPS = 157.3
+# fp32 vector: 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2.4 GHz = 78.6 TFLOP/s.  The
+# published 157.3 counts packed fp32 (two FMAs per lane per instruction); the kernels are built
+# without packed instructions, so 78.6 is the ceiling they can reach and the peak used here.
+PEAK_FP32_VALU_TFLOPS = 78.6
+# quasi-DEER gains about one exact leading step per update, so a solve may need up to T + 1
+# updates; beyond this many passes per solve the run would not finish in a benchmark's time
+QUASI_MAX_PASSES = 20000
 
 
 def log(*a):
@@ -50,8 +57,20 @@ def _plrnn_step(D, model, xd, c, ws_s, ws_a, T_w=0):
     return sum(res["iters"])
 
 
+def check_quasi_bound(c, passes):
+    """Refuse, before any GPU work, a quasi-DEER solve to tolerance whose pass bound (T + 2:
+    about one more exact leading step per update) is too long for a benchmark run; a fixed
+    number of passes is always accepted."""
+    if passes < 0:
+        raise SystemExit("--quasi-passes must be >= 0")
+    if passes == 0 and not c.fixed_iters and c.T + 2 > QUASI_MAX_PASSES:
+        raise SystemExit(f"quasi-DEER on {c.name}: a solve to tolerance may take up to T + 2 = {c.T + 2} passes "
+                         f"(> {QUASI_MAX_PASSES}); pass --quasi-passes K to time K passes per solve instead")
+
+
 def _quasi_step(D, model, xd, c, ws_s, ws_a):
     # quasi-DEER: one more leading step is exact per update, so T + 1 updates always suffice
+    # (check_quasi_bound has refused the workloads where that is too many)
     res = D.deer_solve_quasi(model, xd, c.alpha, c.n_obs, tol=c.tol, max_iter=c.T + 2, fixed_iters=c.fixed_iters,
                              ws=ws_s, check=False)
     if res["status"] != 0:
@@ -194,45 +213,95 @@ def roofline_for(name, c, total_ms, launches, steps, updates):
     return base
 
 
-def cpu_baseline(c, budget_s=20.0):
-    """The float64 oracle on the host, on a bounded sample of the same workload."""
+def _oracle_sample(kind, params, x, alpha, n_obs, tol, max_iter, fixed_iters):
+    """One oracle run on a sample: the work one CPU user of the method would do.  PLRNN kinds:
+    Newton solve, adjoint and parameter gradients; diagonal SSM: forward scan, read-out,
+    reverse scan and gradients.  Returns (timesteps processed, seconds)."""
     import oracle as O
     try:
         from threadpoolctl import threadpool_limits
-        lim = threadpool_limits(1)
+        threadpool_limits(1)
     except Exception:       # pragma: no cover
-        lim = None
-    m = {"kind": c.kind, **c.params}
-    if c.kind == "diag_ssm":
-        Ts = min(c.T, 1 << 16)
-        xs = c.x[:1, :Ts + 1]
-        t0 = time.perf_counter()
-        O.diag_ssm_step(c.params, xs)
-        dt = time.perf_counter() - t0
-        value, sample = Ts / dt, f"1 of {c.B} sequences, first {Ts} of {c.T} steps, forward+read-out+reverse"
+        pass
+    t0 = time.perf_counter()
+    if kind == "diag_ssm":
+        O.diag_ssm_step(params, x)
+        work = x.shape[0] * (x.shape[1] - 1)
     else:
-        # The oracle is vectorised over the batch and sequential in time.  Calibrate on a short
-        # prefix, then keep the whole batch and shorten T to fit the budget.
-        Tc = min(c.T, 512)
-        t0 = time.perf_counter()
-        rc = O.newton(m, c.x[:, :Tc + 1], c.alpha, c.n_obs, tol=c.tol, max_iter=c.max_iter,
-                      fixed_iters=c.fixed_iters)
-        per = (time.perf_counter() - t0) / (Tc * max(1, int(rc["iters"].max())))
+        m = {"kind": kind, **params}
+        res = O.newton(m, x, alpha, n_obs, tol=tol, max_iter=max_iter, fixed_iters=fixed_iters)
+        lam = O.adjoint(m, x, res["z"], alpha, n_obs)
+        O.param_grads(m, x, res["z"], alpha, n_obs, lam)
+        work = float(np.sum(res["iters"])) * (x.shape[1] - 1)
+    return work, time.perf_counter() - t0
+
+
+def _warm_worker(_):
+    import oracle  # noqa: F401  (import cost kept out of the timed region)
+    return os.getpid()
+
+
+def _host_cpu():
+    """Usable host cores (affinity) and the CPU model name."""
+    try:
+        ncpu = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        ncpu = os.cpu_count() or 1
+    model = "unknown"
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:         # pragma: no cover
+        pass
+    return ncpu, model
+
+
+def cpu_baseline(c, budget_s=12.0, max_workers=16):
+    """The float64 oracle on the host, on a bounded sample of the same workload, twice: on one
+    thread, and across the host's cores with one worker process per share of the sequences
+    (at most B workers, at most `max_workers`; each worker single-threaded).  Runs in child
+    processes of this one, before the GPU is used."""
+    import multiprocessing as mp
+    ncpu, model = _host_cpu()
+    args = (c.kind, c.params, None, c.alpha, c.n_obs, c.tol, c.max_iter, c.fixed_iters)
+    if c.kind == "diag_ssm":
+        Ts = min(c.T, 1 << 15)
+        seqs = list(range(c.B))
+        single_x = c.x[:1, :Ts + 1]
+        desc = f"first {Ts} of {c.T} steps, forward + read-out + reverse + gradients"
+    else:
+        # calibrate on a short prefix of the whole batch, then shorten T to fit the budget
+        Tc = min(c.T, 256)
+        w, dt = _oracle_sample(*args[:2], c.x[:, :Tc + 1], *args[3:])
+        per = dt / max(w, 1.0)          # seconds per (b, t, update)
         Ts = c.T
-        while Ts > 1024 and Ts * per * 12 > budget_s:
+        while Ts > 512 and per * w / Tc * Ts > budget_s:
             Ts //= 2
-        xs = c.x[:, :Ts + 1]
+        seqs = list(range(c.B))
+        single_x = c.x[:, :Ts + 1]
+        desc = f"first {Ts} of {c.T} steps, Newton solve + adjoint + gradients"
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(1) as pool:
+        w1, dt1 = pool.apply(_oracle_sample, (*args[:2], np.ascontiguousarray(single_x), *args[3:]))
+    nw = max(1, min(len(seqs), ncpu, max_workers))
+    if c.kind == "diag_ssm":
+        shares = [c.x[[b], :Ts + 1] for b in seqs]
+        desc_all = f"all {c.B} sequences, " + desc
+    else:
+        shares = [c.x[seqs[k::nw], :Ts + 1] for k in range(nw)]
+        desc_all = f"all {c.B} sequences, " + desc
+    with ctx.Pool(nw) as pool:
+        pool.map(_warm_worker, range(nw))
         t0 = time.perf_counter()
-        res = O.newton(m, xs, c.alpha, c.n_obs, tol=c.tol, max_iter=c.max_iter, fixed_iters=c.fixed_iters)
-        lam = O.adjoint(m, xs, res["z"], c.alpha, c.n_obs)
-        O.param_grads(m, xs, res["z"], c.alpha, c.n_obs, lam)
-        dt = time.perf_counter() - t0
-        value = float(np.sum(res["iters"]) * Ts) / dt
-        sample = f"all {c.B} sequences, first {Ts} of {c.T} steps, Newton solve + adjoint + gradients"
-    if lim is not None:
-        lim.unregister() if hasattr(lim, "unregister") else None
-    return {"value": value, "unit": "timesteps/s", "cores": 1, "kind": "oracle", "sample": sample,
-            "seconds": dt, "host_cpus": os.cpu_count()}
+        res = pool.starmap(_oracle_sample, [(*args[:2], np.ascontiguousarray(x), *args[3:]) for x in shares])
+        dtn = time.perf_counter() - t0
+    wn = sum(r[0] for r in res)
+    single = {"value": w1 / dt1, "cores": 1, "seconds": dt1,
+              "sample": (f"1 of {c.B} sequences, " if c.kind == "diag_ssm" else f"all {c.B} sequences, ") + desc}
+    return {"value": wn / dtn, "unit": "timesteps/s", "cores": nw, "kind": "oracle", "sample": desc_all,
+            "seconds": dtn, "single_thread": single, "host_cpus": ncpu, "cpu_model": model}
 
 
 def fig1a_sweep(reps: int = 3):
@@ -303,7 +372,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
+    ap.add_argument("--config", type=int, default=5, help="workload 1..5 (default 5, the M = 64 vanilla PLRNN)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--tw", type=int, default=0,
                     help="PLRNN workloads with a tolerance: latent warm-up of this many steps")
@@ -312,6 +381,9 @@ def main():
                          "MAR, gradient, Adam update in place)")
     ap.add_argument("--quasi", action="store_true",
                     help="PLRNN workloads: quasi-DEER (diagonal Jacobians) instead of GTF-DEER")
+    ap.add_argument("--quasi-passes", type=int, default=0,
+                    help="with --quasi: run exactly this many quasi-DEER updates per solve (no tolerance) and "
+                         "report that throughput; required when T + 2 exceeds %d" % QUASI_MAX_PASSES)
     ap.add_argument("--fig1a", action="store_true",
                     help="instead of the workload: the Fig. 1A sweep, GTF-DEER against the sequential baseline")
     args = ap.parse_args()
@@ -330,6 +402,20 @@ def main():
 
     c = W.make_config(args.config)
     log(f"[bench] workload {c.name}: B={c.B} T={c.T} M={c.M} kind={c.kind}")
+    if args.quasi:
+        if c.kind != "plrnn":
+            print("quasi-DEER is built for the vanilla PLRNN workloads (1, 2, 5)", file=sys.stderr)
+            sys.exit(3)
+        check_quasi_bound(c, args.quasi_passes)
+        if args.quasi_passes > 0:
+            c.fixed_iters = args.quasi_passes
+    cb = None
+    if not args.no_cpu_baseline and not args.quasi:
+        # before the GPU is used: the oracle runs in child processes of this one
+        log("[bench] timing the CPU oracle on a bounded sample (one thread, then all cores)")
+        cb = cpu_baseline(c)
+        log(f"[bench] cpu oracle: {cb['single_thread']['value']:.4g} timesteps/s on 1 thread, {cb['value']:.4g} on "
+            f"{cb['cores']} processes ({cb['cpu_model']}, {cb['host_cpus']} usable cpus; {cb['sample']})")
     dev = torch.device("cuda:0")
     xd = torch.tensor(c.x, device=dev)
     # a plain device copy of known size: the calibration the counter passes scale by
@@ -353,9 +439,6 @@ def main():
             tstate = {"step": 0}
             step = lambda: _train_step(D, model, xd, c, ws_t, tstate, args.tw)   # noqa: E731
         elif args.quasi:
-            if c.kind != "plrnn":
-                print("quasi-DEER is built for the vanilla PLRNN workloads (1, 2, 5)", file=sys.stderr)
-                sys.exit(3)
             lib = D.load()
             ws_s = D._workspace(lib.deer_quasi_workspace_bytes(ctypes.byref(model.c), c.B, c.T, Bnd.DEER_OP_SOLVE))
             ws_a = D._workspace(lib.deer_quasi_workspace_bytes(ctypes.byref(model.c), c.B, c.T,
@@ -373,10 +456,14 @@ def main():
         print(f"workload {c.name}: model kind {c.kind} not supported by this build", file=sys.stderr)
         sys.exit(3)
 
+    t_w = time.perf_counter()
     for i in range(args.warmup):
         step()
-        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done ({time.perf_counter() - t_w:.2f} s)")
     torch.cuda.synchronize()
+    # steps long enough to be seen are reported one by one (outside the timed region for short ones)
+    slow = args.warmup > 0 and (time.perf_counter() - t_w) / args.warmup > 0.5
     # per-kernel durations: HIP events around every launch on the stream it is launched on,
     # over separate steps (the events add launch overhead, so the timed steps run without them)
     prof_steps = max(1, min(args.steps, 3))
@@ -384,6 +471,8 @@ def main():
     prof_updates = 0
     for i in range(prof_steps):
         prof_updates += step()
+        if slow:
+            log(f"[bench] event-timed step {i + 1}/{prof_steps} done")
     torch.cuda.synchronize()
     kt = Bnd.timing_report()
     Bnd.timing_enable(False)
@@ -392,8 +481,11 @@ def main():
     updates = 0
     for i in range(args.steps):
         updates += step()
+        if slow:
+            log(f"[bench] timed step {i + 1}/{args.steps} returned")
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    log(f"[bench] {args.steps} timed steps: {(t1 - t0) * 1e3 / args.steps:.3f} ms per step")
     dt = t1 - t0
     iters_per_step = updates / args.steps
     timesteps = updates * c.T
@@ -432,11 +524,8 @@ def main():
         "roofline": roof,
         "kernels": kernels,
     }
-    if not args.no_cpu_baseline and not args.quasi:
-        log("[bench] timing the CPU oracle on a bounded sample")
-        cb = cpu_baseline(c)
+    if cb is not None:
         out["cpu_baseline"] = cb
-        log(f"[bench] cpu oracle: {cb['value']:.4g} timesteps/s ({cb['sample']}, {cb['seconds']:.1f} s)")
     print(json.dumps(out), flush=True)
 
 

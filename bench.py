@@ -189,6 +189,31 @@ def measured_traffic(workload, kernel):
     return float(rec["traffic_bytes_per_launch"])
 
 
+def measured_mfma(workload, kernel):
+    """Matrix-core activity of the kernel from rocprofv3 counter passes
+    (SQ_INSTS_VALU_MFMA_MOPS_F32, SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE), kept in
+    profiles/mfma_<workload>.txt with the hash of the kernel's source; None once it changed."""
+    import hashlib
+    path = os.path.join(HERE, "profiles", f"mfma_{workload}.txt")
+    if not os.path.exists(path) or kernel not in KERNEL_SOURCE:
+        return None
+    rec = {}
+    for ln in open(path):
+        if ":" in ln and not ln.startswith("#"):
+            k, v = ln.split(":", 1)
+            rec[k.strip()] = v.strip()
+    src = os.path.join(HERE, "paper_2605_12683_amd", "csrc", KERNEL_SOURCE[kernel])
+    if rec.get("kernel") != kernel or not os.path.exists(src):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("source_sha256"):
+        return None
+    tf = float(rec["mfma_counted_tflops"])
+    return {"busy_frac": float(rec["mfma_busy_frac"]), "counted_tflops": tf,
+            "counted_frac": tf / PEAK_FP32_MFMA_TFLOPS,
+            "counted_flops_per_launch": float(rec["mfma_flops_per_dispatch"]),
+            "source": f"profiles/mfma_{workload}.txt"}
+
+
 def roofline_for(name, c, total_ms, launches, steps, updates):
     """Algorithmic work of the dominant kernel over the timed region, divided by its time."""
     work = kernel_work(c, steps, updates)
@@ -201,7 +226,8 @@ def roofline_for(name, c, total_ms, launches, steps, updates):
     if bound == "mfma":
         ach = w / (total_ms * 1e-3) / 1e12
         base.update({"bound": "mfma", "achieved": ach, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": ach / PEAK_FP32_MFMA_TFLOPS, "work_per_launch": w / launches})
+                     "frac": ach / PEAK_FP32_MFMA_TFLOPS, "work_per_launch": w / launches,
+                     "mfma_counters": measured_mfma(c.name, name)})
     elif bound == "alu":
         ach = w / (total_ms * 1e-3) / 1e12
         base.update({"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS, "unit": "TFLOP/s",

@@ -36,9 +36,18 @@
  *  - Errors are returned as a status code (never thrown across the ABI);
  *    argument errors are detected before any device work is queued.
  *    deer_last_error() gives a thread-local message for the last failure.
- *  - The library keeps no mutable global state; calls on different streams
- *    with different workspaces may run concurrently.  Calls that share a
- *    workspace must be serialised by the caller.
+ *  - Process-wide state (nothing else is kept between calls):
+ *      * one pinned host block per host thread, through which the device reports
+ *        stopped sequences to the Newton loop of a solve with a tolerance; it is
+ *        allocated only by deer_host_reserve and freed by deer_host_release, never
+ *        inside a solve;
+ *      * the timing diagnostics (deer_timing_*), off unless enabled, which keep a
+ *        mutex-protected pool of HIP events;
+ *      * the read-out's resident-block count (an occupancy query made once per
+ *        process).
+ *    Calls on different streams with different workspaces may run concurrently;
+ *    calls that share a workspace must be serialised by the caller, and one host
+ *    thread runs its solves one at a time.
  */
 #ifndef DEER_H
 #define DEER_H
@@ -141,9 +150,10 @@ size_t deer_workspace_bytes_ex(const deer_model *model, const deer_forcing *forc
  *   final_norm   host [B] out or NULL: max |Delta z| of each sequence's last update.
  * Each Newton update is applied before the test; a sequence whose update is below tol
  * is frozen while the others continue.  With fixed_iters == 0 the test runs on the device
- * after every update; a sequence that stops clears a flag in a pinned host block of the
- * calling thread (allocated on first use, grown with B, kept until the process ends) that
- * also receives its update count, last norm and status.  The host keeps passes queued ahead
+ * after every update; a sequence that stops clears a flag in the calling thread's pinned host
+ * block (deer_host_reserve(B) must have been called on this thread; otherwise the call returns
+ * DEER_ERR_INVALID_ARG before any device work), which also receives its update count, last
+ * norm and status.  The host keeps passes queued ahead
  * of the device and returns once every sequence has stopped (then without a stream
  * synchronisation: z is complete in stream order, and the passes still queued skip every
  * sequence) or at max_iter (after a synchronisation).  Calls from one host thread run one
@@ -311,19 +321,39 @@ int plrnn_jacobian(const deer_model *model, const deer_forcing *forcing, int B, 
 
 /* The bare associative scan over affine pairs (scheduled-sampling appendix: the pair
  * (A_t, b_t) and its composition), batched over B independent sequences of length T.
- *   DEER_SCAN_DENSE:    J [B,T,M,M], b [B,T,M], M <= 64.
- *        reverse == 0:  y_t = J_t y_{t-1} + b_t, y_0 = 0        (J_1 is not read)
- *        reverse != 0:  y_T = b_T, y_{t-1} = J_t^T y_t + b_{t-1}  (J_1 is not read)
- *   DEER_SCAN_DIAG_C64: J = lambda [M][2], b [B,T,M][2] complex.
- *        reverse == 0:  y_t = lambda y_{t-1} + b_t, y_0 = 0
- *        reverse != 0:  y_T = b_T, y_{t-1} = conj(lambda) y_t + b_{t-1}
+ * `reverse` chooses the direction, `transpose` whether each step applies its matrix (0) or
+ * its transpose (1); the Newton update of eq. GTF_DEER_update is (reverse, transpose) = (0, 0)
+ * and the adjoint recursion of eq. backward_recursion is (1, 1).  With op(J) = J or J^T:
+ *   DEER_SCAN_DENSE:    J [B,T,M,M] row-major per step, b [B,T,M], M <= 64.
+ *        reverse == 0:  y_t = op(J_t) y_{t-1} + b_t, y_0 = 0        (J_1 is not read)
+ *        reverse != 0:  y_T = b_T, y_{t-1} = op(J_t) y_t + b_{t-1}  (J_1 is not read)
+ *   DEER_SCAN_DIAG_C64: J = lambda [M][2], b [B,T,M][2] complex; op(lambda) = lambda, or
+ *        conj(lambda) with transpose != 0 (C read as R^2, where multiplication by lambda is
+ *        the 2 x 2 block [[Re, -Im], [Im, Re]] and its transpose is multiplication by conj):
+ *        reverse == 0:  y_t = op(lambda) y_{t-1} + b_t, y_0 = 0
+ *        reverse != 0:  y_T = b_T, y_{t-1} = op(lambda) y_t + b_{t-1}
  *   y     out, same layout as b (may not alias b).
- * Fully asynchronous. */
-int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, const float *b, float *y,
-              void *ws, size_t ws_bytes, void *stream);
+ * The scan takes explicit matrices; the mask-driven Jacobians of the PLRNN kinds are formed
+ * inside deer_solve / deer_adjoint, which know the model.  Fully asynchronous. */
+int deer_scan(int layout, int reverse, int transpose, int B, int T, int M, const float *J, const float *b,
+              float *y, void *ws, size_t ws_bytes, void *stream);
 
-/* Workspace bytes deer_scan needs. */
-size_t deer_scan_workspace_bytes(int layout, int B, int T, int M);
+/* Workspace bytes deer_scan needs for these arguments (0 if they are invalid). */
+size_t deer_scan_workspace_bytes(int layout, int reverse, int transpose, int B, int T, int M);
+
+/* Reserves the calling host thread's pinned host block for solves with a tolerance of up to
+ * max_batch sequences (deer_solve, deer_solve_quasi, deer_train_step): (4 max_batch + 32)
+ * 32-bit words of device-coherent pinned host memory, through which the device reports each
+ * sequence that stops (its flag, update count, last norm and status) and the start of each
+ * forward pass, so the host follows the Newton loop without copies or stream synchronisation.
+ * A block that already holds max_batch sequences is kept (no call); a smaller one is replaced.
+ * Call it once per thread at set-up, outside any solve of that thread.  Returns DEER_OK,
+ * DEER_ERR_INVALID_ARG (max_batch <= 0) or DEER_ERR_HIP (the pinned allocation failed). */
+int deer_host_reserve(int max_batch);
+
+/* Frees the calling thread's pinned host block (no-op without one); a later solve with a
+ * tolerance on this thread needs deer_host_reserve again. */
+int deer_host_release(void);
 
 /* Diagnostics: per-kernel timing with HIP events.  While enabled, every kernel launch is
  * bracketed by two events recorded on the stream it is launched on (the caller's stream).

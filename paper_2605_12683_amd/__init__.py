@@ -13,6 +13,7 @@ Model dictionaries use the paper's names:
 from __future__ import annotations
 
 import ctypes
+import threading
 
 import torch
 
@@ -21,7 +22,8 @@ from ._binding import DeerError, load  # noqa: F401
 
 __all__ = ["deer_solve", "deer_adjoint", "deer_readout_loss", "plrnn_jacobian", "deer_scan", "deer_workspace_bytes",
            "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_status_string", "DeerError", "load",
-           "deer_sequential", "deer_sequential_workspace_bytes", "deer_solve_quasi", "deer_adjoint_quasi", "deer_train_step"]
+           "deer_sequential", "deer_sequential_workspace_bytes", "deer_solve_quasi", "deer_adjoint_quasi", "deer_train_step",
+           "deer_host_reserve"]
 
 _KINDS = {"plrnn": _b.DEER_PLRNN, "shplrnn": _b.DEER_SHPLRNN, "diag_ssm": _b.DEER_DIAG_SSM}
 _INITS = {"teacher": _b.DEER_INIT_TEACHER, "zero": _b.DEER_INIT_ZERO, "user": _b.DEER_INIT_USER}
@@ -44,6 +46,18 @@ def _dev(t, dtype=torch.float32):
 
 def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+_host = threading.local()
+
+
+def deer_host_reserve(B: int) -> None:
+    """Reserve the calling thread's pinned host block for solves of up to B sequences
+    (deer_host_reserve in the C ABI; the solves themselves allocate nothing)."""
+    if getattr(_host, "cap", 0) >= B:
+        return
+    _b._check(load().deer_host_reserve(int(B)), "deer_host_reserve")
+    _host.cap = int(B)
 
 
 class _Model:
@@ -136,8 +150,9 @@ def deer_workspace_bytes(model, B: int, T: int, op: int) -> int:
     return int(load().deer_workspace_bytes(ctypes.byref(m.c), B, T, op))
 
 
-def deer_scan_workspace_bytes(layout: int, B: int, T: int, M: int) -> int:
-    return int(load().deer_scan_workspace_bytes(layout, B, T, M))
+def deer_scan_workspace_bytes(layout: int, B: int, T: int, M: int, reverse: bool = False, transpose=None) -> int:
+    tr = reverse if transpose is None else transpose
+    return int(load().deer_scan_workspace_bytes(layout, int(bool(reverse)), int(bool(tr)), B, T, M))
 
 
 def _workspace(nbytes: int):
@@ -188,6 +203,8 @@ def _solve(entry, quasi, model, x, alpha, n_forced, *, z0, tol, max_iter, fixed_
     iters = (ctypes.c_int32 * B)()
     norms = (ctypes.c_float * B)()
     o = _b.deer_solve_opts(float(tol), int(max_iter), int(fixed_iters), _INITS[init], float(step_bound))
+    if m.kind != "diag_ssm" and int(fixed_iters) <= 0:
+        deer_host_reserve(B)
     z0d = _dev(z0)
     st = getattr(lib, entry)(ctypes.byref(m.c), ctypes.byref(f), ctypes.byref(o), B, T, _ptr(x), _ptr(z0d),
                              _ptr(out), _ptr(masks), iters, norms, _ptr(ws), ws.numel(), _stream())
@@ -297,6 +314,7 @@ def deer_train_step(model, x, alpha: float, n_forced: int, *, step: int, state=N
     iters = (ctypes.c_int32 * B)()
     grads, gs = _plrnn_grads(m) if want_grads else ({}, None)
     z0d = _dev(z0)
+    deer_host_reserve(B)
     st = lib.deer_train_step(ctypes.byref(m.c), ctypes.byref(f), ctypes.byref(o), ctypes.byref(tr), B, T, _ptr(x),
                              _ptr(z0d), _ptr(z), _ptr(state["m"]), _ptr(state["v"]),
                              ctypes.byref(gs) if gs is not None else None, _ptr(loss), iters, _ptr(ws), ws.numel(),
@@ -367,16 +385,19 @@ def plrnn_jacobian(model, x, z, alpha: float, n_forced: int, *, z0=None, want=("
     return out
 
 
-def deer_scan(layout: int, J, b, reverse: bool = False, ws=None):
-    """Bare affine scan (DEER_SCAN_DENSE: J [B,T,M,M]; DEER_SCAN_DIAG_C64: lambda [M] complex)."""
+def deer_scan(layout: int, J, b, reverse: bool = False, ws=None, transpose=None):
+    """Bare affine scan (DEER_SCAN_DENSE: J [B,T,M,M]; DEER_SCAN_DIAG_C64: lambda [M] complex).
+    transpose defaults to `reverse` (the adjoint's orientation)."""
     lib = load()
     J = _dev(J)
     b = _dev(b)
     B, T, M = b.shape[:3]
+    tr = reverse if transpose is None else transpose
     y = torch.empty_like(b)
     if ws is None:
-        ws = _workspace(lib.deer_scan_workspace_bytes(layout, B, T, M))
-    st = lib.deer_scan(layout, 1 if reverse else 0, B, T, M, _ptr(J), _ptr(b), _ptr(y), _ptr(ws), ws.numel(),
-                       _stream())
+        ws = _workspace(lib.deer_scan_workspace_bytes(layout, int(bool(reverse)), int(bool(tr)), B, T, M))
+    st = lib.deer_scan(layout, 1 if reverse else 0, 1 if tr else 0, B, T, M, _ptr(J), _ptr(b), _ptr(y), _ptr(ws),
+                       ws.numel(), _stream())
     _b._check(st, "deer_scan")
     return y
+

@@ -25,7 +25,8 @@ EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "deer_adjoint_
             "deer_scan_workspace_bytes", "deer_readout_workspace_bytes", "deer_readout_loss", "deer_status_string",
             "deer_last_error", "deer_timing_enable", "deer_timing_report", "deer_solve_quasi", "deer_adjoint_quasi",
             "deer_quasi_workspace_bytes", "deer_sequential", "deer_sequential_workspace_bytes",
-            "deer_workspace_bytes_ex", "deer_train_step", "deer_train_workspace_bytes", "deer_train_params"]
+            "deer_workspace_bytes_ex", "deer_train_step", "deer_train_workspace_bytes", "deer_train_params",
+            "deer_host_reserve", "deer_host_release"]
 
 _fp = ctypes.c_void_p
 
@@ -79,7 +80,7 @@ def load(path: str = LIB_PATH):
     sz, i32, vp = ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p
     lib.deer_workspace_bytes.argtypes = [P(deer_model), i32, i32, i32]
     lib.deer_workspace_bytes.restype = sz
-    lib.deer_scan_workspace_bytes.argtypes = [i32, i32, i32, i32]
+    lib.deer_scan_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
     lib.deer_scan_workspace_bytes.restype = sz
     lib.deer_solve.argtypes = [P(deer_model), P(deer_forcing), P(deer_solve_opts), i32, i32, vp, vp, vp, vp,
                                P(ctypes.c_int32), P(ctypes.c_float), vp, sz, vp]
@@ -117,8 +118,12 @@ def load(path: str = LIB_PATH):
     lib.deer_readout_loss.restype = i32
     lib.plrnn_jacobian.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.plrnn_jacobian.restype = i32
-    lib.deer_scan.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]
+    lib.deer_scan.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]
     lib.deer_scan.restype = i32
+    lib.deer_host_reserve.argtypes = [i32]
+    lib.deer_host_reserve.restype = i32
+    lib.deer_host_release.argtypes = []
+    lib.deer_host_release.restype = i32
     lib.deer_status_string.argtypes = [i32]
     lib.deer_status_string.restype = ctypes.c_char_p
     lib.deer_last_error.argtypes = []

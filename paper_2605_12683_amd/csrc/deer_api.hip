@@ -577,8 +577,8 @@ constexpr float kDefaultStepBound = 1e3f;
 constexpr NewtonDamp kDamp = {1.f / 64, 4.f, 4.f, 1e-4f};
 constexpr int kFirstBatch = 4, kBatch = 1;
 
-// Pinned, device-coherent host block of the Newton loop, one per host thread (grown on
-// demand, kept for the life of the process): act | it | norm | status (cap words each; see
+// Pinned, device-coherent host block of the Newton loop, one per host thread, reserved by
+// deer_host_reserve (the solves allocate nothing): act | it | norm | status (cap words each; see
 // NewtonDev), then the pass mark.  Passes are numbered per thread; the M <= 16 forward pass
 // writes its number to the mark as it starts.
 struct HostBlk {
@@ -587,16 +587,32 @@ struct HostBlk {
     uint32_t next_pass = 1;   // number of the next marked pass
 };
 static thread_local HostBlk t_host;
+
+static int host_reserve(int B) {
+    if ((size_t)B <= t_host.cap) return DEER_OK;
+    if (t_host.base) (void)hipHostFree(t_host.base);
+    t_host.base = nullptr;
+    t_host.cap = 0;
+    DEER_HIP(hipHostMalloc((void **)&t_host.base, (4 * (size_t)B + 32) * sizeof(int), hipHostMallocCoherent));
+    t_host.cap = (size_t)B;
+    // no pass of this thread is pending (every earlier solve returned after its last mark)
+    *(uint32_t *)(t_host.base + 4 * t_host.cap) = t_host.next_pass - 1;
+    return DEER_OK;
+}
+
+// A solve with a tolerance needs the calling thread's block to hold B sequences; checked before
+// any device work is queued.
+static int check_host_reserved(int B) {
+    if ((size_t)B <= t_host.cap) return DEER_OK;
+    set_error("solves with a tolerance report through a pinned host block of the calling thread: it holds %zu "
+              "sequences, %d are needed (call deer_host_reserve(%d) on this thread first)",
+              t_host.cap, B, B);
+    return DEER_ERR_INVALID_ARG;
+}
+
 static int host_block(int B, NewtonDev &nd, uint32_t **mark) {
-    if ((size_t)B > t_host.cap) {
-        if (t_host.base) (void)hipHostFree(t_host.base);
-        t_host.base = nullptr;
-        t_host.cap = 0;
-        DEER_HIP(hipHostMalloc((void **)&t_host.base, (4 * (size_t)B + 32) * sizeof(int), hipHostMallocCoherent));
-        t_host.cap = (size_t)B;
-        // no pass of this thread is pending (every earlier solve returned after its last mark)
-        *(uint32_t *)(t_host.base + 4 * t_host.cap) = t_host.next_pass - 1;
-    }
+    int rc = check_host_reserved(B);
+    if (rc) return rc;
     int *p = t_host.base;
     const size_t cap = t_host.cap;
     nd.hact = p;
@@ -1109,6 +1125,23 @@ const char *deer_status_string(int s) {
 
 const char *deer_last_error(void) { return g_err; }
 
+int deer_host_reserve(int max_batch) {
+    set_error("");
+    if (max_batch <= 0) { set_error("max_batch must be positive"); return DEER_ERR_INVALID_ARG; }
+    return host_reserve(max_batch);
+}
+
+int deer_host_release(void) {
+    set_error("");
+    if (t_host.base) {
+        hipError_t e = hipHostFree(t_host.base);
+        t_host.base = nullptr;
+        t_host.cap = 0;
+        if (e != hipSuccess) return hip_fail(e, "hipHostFree");
+    }
+    return DEER_OK;
+}
+
 int deer_timing_enable(int on) {
     TimingState &s = tstate();
     std::lock_guard<std::mutex> g(s.mu);
@@ -1163,7 +1196,9 @@ size_t deer_workspace_bytes(const deer_model *m, int B, int T, int op) {
     return 0;
 }
 
-size_t deer_scan_workspace_bytes(int layout, int B, int T, int M) {
+size_t deer_scan_workspace_bytes(int layout, int reverse, int transpose, int B, int T, int M) {
+    (void)reverse;
+    (void)transpose;
     if (B <= 0 || T <= 0 || M <= 0) return 0;
     if (layout == DEER_SCAN_DIAG_C64) return diag_scan_ws_bytes(B, T, M);
     if (layout == DEER_SCAN_DENSE && M <= 64) {
@@ -1209,6 +1244,7 @@ int deer_solve(const deer_model *m, const deer_forcing *f, const deer_solve_opts
     if (!o || !x || !z) { set_error("opts, x and z are required"); return DEER_ERR_INVALID_ARG; }
     if (o->init < 0 || o->init > 2) { set_error("unknown init %d", o->init); return DEER_ERR_INVALID_ARG; }
     if (!(o->tol >= 0.f) && o->fixed_iters <= 0) { set_error("tol must be >= 0"); return DEER_ERR_INVALID_ARG; }
+    if (m->kind != DEER_DIAG_SSM && o->fixed_iters <= 0 && (rc = check_host_reserved(B))) return rc;
     hipStream_t st = (hipStream_t)stream;
     if (f->T_w > 0) return solve_warmup(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st, false);
     if (m->kind == DEER_PLRNN)
@@ -1334,6 +1370,7 @@ int deer_solve_quasi(const deer_model *m, const deer_forcing *f, const deer_solv
     if (!o || !x || !z) { set_error("opts, x and z are required"); return DEER_ERR_INVALID_ARG; }
     if (o->init < 0 || o->init > 2) { set_error("unknown init %d", o->init); return DEER_ERR_INVALID_ARG; }
     if (!(o->tol >= 0.f) && o->fixed_iters <= 0) { set_error("tol must be >= 0"); return DEER_ERR_INVALID_ARG; }
+    if (o->fixed_iters <= 0 && (rc = check_host_reserved(B))) return rc;
     if (f->T_w > 0)
         return solve_warmup(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, (hipStream_t)stream, true);
     return solve_quasi(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, (hipStream_t)stream);
@@ -1409,6 +1446,7 @@ int deer_train_step(const deer_model *m, const deer_forcing *f, const deer_solve
     if (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN) { set_error("deer_train_step: PLRNN kinds only"); return DEER_ERR_INVALID_ARG; }
     if (!o || !tr || !x || !z || !adam_m || !adam_v) { set_error("opts, train, x, z and the Adam moments are required"); return DEER_ERR_INVALID_ARG; }
     if (o->fixed_iters > 0) { set_error("deer_train_step solves to a tolerance (fixed_iters = 0)"); return DEER_ERR_INVALID_ARG; }
+    if ((rc = check_host_reserved(B))) return rc;
     if (tr->step < 1 || !(tr->lr > 0.f) || !(tr->beta1 >= 0.f && tr->beta1 < 1.f) || !(tr->beta2 >= 0.f && tr->beta2 < 1.f)) {
         set_error("Adam needs step >= 1, lr > 0 and betas in [0, 1)");
         return DEER_ERR_INVALID_ARG;
@@ -1546,17 +1584,19 @@ int deer_readout_loss(const deer_readout *r, int B, int T, int M, const float *h
     return launch_readout(ra, B, T, h, x, g, masks, loss, gr, ws, (hipStream_t)stream);
 }
 
-int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, const float *b, float *y, void *ws,
-              size_t ws_bytes, void *stream) {
+int deer_scan(int layout, int reverse, int transpose, int B, int T, int M, const float *J, const float *b, float *y,
+              void *ws, size_t ws_bytes, void *stream) {
     set_error("");
     if (B <= 0 || T <= 0 || M <= 0) { set_error("B, T, M must be positive"); return DEER_ERR_INVALID_ARG; }
     if (!J || !b || !y) { set_error("J, b and y are required"); return DEER_ERR_INVALID_ARG; }
     if (b == y) { set_error("y may not alias b"); return DEER_ERR_INVALID_ARG; }
     hipStream_t st = (hipStream_t)stream;
+    const bool rev = reverse != 0, tr = transpose != 0;
     if (layout == DEER_SCAN_DIAG_C64) {
         int rc = check_ws(ws, ws_bytes, diag_scan_ws_bytes(B, T, M));
         if (rc) return rc;
-        return launch_diag_scan(reverse != 0, B, T, M, J, b, nullptr, 0, nullptr, y, ws, st);
+        // the transpose of multiplication by lambda (C read as R^2) is multiplication by conj(lambda)
+        return launch_diag_scan(rev, B, T, M, J, b, nullptr, 0, nullptr, y, ws, st, tr ? 1 : 0);
     }
     if (layout == DEER_SCAN_DENSE) {
         if (M > 64) { set_error("dense scans support M <= 64"); return DEER_ERR_INVALID_ARG; }
@@ -1565,10 +1605,13 @@ int deer_scan(int layout, int reverse, int B, int T, int M, const float *J, cons
         int rc = check_ws(ws, ws_bytes, need);
         if (rc) return rc;
         DenseWs w = carve_dense(ws, B, T, M, &need);
-        const bool rev = reverse != 0;
-        if ((rc = launch_chunk_product_dense(rev, B, T, M, J, b, 1.f, w.P, w.v, nullptr, w.C, w.ncs, st))) return rc;
+        // the kernels' default orientation is J_t forward and J_{t+1}^T in reverse
+        const bool flip = tr != rev;
+        if ((rc = launch_chunk_product_dense(rev, B, T, M, J, b, 1.f, w.P, w.v, nullptr, w.C, w.ncs, st, flip)))
+            return rc;
         if ((rc = launch_carry(w.MP, rev, w.P, w.v, w.carry, nullptr, nullptr, B, w.ncs, w.gws, st))) return rc;
-        return launch_fixup_dense(rev ? 2 : 1, B, T, M, J, b, 1.f, w.carry, nullptr, y, nullptr, nullptr, nullptr, w.C, w.ncs, st);
+        return launch_fixup_dense(rev ? 2 : 1, B, T, M, J, b, 1.f, w.carry, nullptr, y, nullptr, nullptr, nullptr, w.C,
+                                  w.ncs, st, flip);
     }
     set_error("deer_scan: unknown layout %d", layout);
     return DEER_ERR_INVALID_ARG;

@@ -27,7 +27,10 @@ __device__ __forceinline__ float jload(const float *__restrict__ Jp, int M, int 
     return (row < M && col < M) ? Jp[row * M + col] : 0.f;
 }
 
-template <int MP, bool REV>
+// FLIP: the scan uses the other orientation of every stored matrix than the direction's default
+// (forward: J_t^T instead of J_t; reverse: J_{t+1} instead of J_{t+1}^T), so one kernel serves all
+// four (direction, transpose) combinations of the bare scan.
+template <int MP, bool REV, bool FLIP>
 __global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restrict__ J, const float *__restrict__ rhs,
                                                             float rhs_sign, float *__restrict__ Pout,
                                                             float *__restrict__ vout, const int *__restrict__ active,
@@ -85,7 +88,9 @@ __global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restr
 #pragma unroll
                     for (int j = 0; j < NS / 4; ++j)
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) Aop[I][4 * j + q] = jload(Jp, M, 16 * I + c, 16 * j + 4 * g + q);
+                        for (int q = 0; q < 4; ++q)
+                            Aop[I][4 * j + q] = FLIP ? jload(Jp, M, 16 * j + 4 * g + q, 16 * I + c)
+                                                     : jload(Jp, M, 16 * I + c, 16 * j + 4 * g + q);
                 float Bop[NS];
 #pragma unroll
                 for (int j = 0; j < NS / 4; ++j)
@@ -108,9 +113,11 @@ __global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restr
             lds_barrier();
             float y = 0.f;
             if (run && ui < M) {
-                const float *Jr = J + (((size_t)ub * T + s) * M + ui) * M;
+                // row ui of J_s, or column ui when flipped
+                const float *Jr = FLIP ? J + ((size_t)ub * T + s) * M * M + ui : J + (((size_t)ub * T + s) * M + ui) * M;
+                const size_t stride = FLIP ? (size_t)M : 1;
                 const float *l = lds + un * MP;
-                for (int k = 0; k < M; ++k) y = fmaf(Jr[k], l[k], y);
+                for (int k = 0; k < M; ++k) y = fmaf(Jr[k * stride], l[k], y);
             }
             lds_barrier();
             if (run && ui < M) u = fmaf(rhs_sign, rhs[((size_t)ub * T + s) * M + ui], y);
@@ -120,9 +127,11 @@ __global__ __launch_bounds__(64) void k_chunk_product_dense(const float *__restr
             lds_barrier();
             float y = 0.f;
             if (run && ui < M && t > 0) {
-                const float *Jc = J + ((size_t)ub * T + k + 1) * M * M + ui;
+                // column ui of J_{k+1}, or row ui when flipped
+                const float *Jc = FLIP ? J + (((size_t)ub * T + k + 1) * M + ui) * M : J + ((size_t)ub * T + k + 1) * M * M + ui;
+                const size_t stride = FLIP ? 1 : (size_t)M;
                 const float *l = lds + un * MP;
-                for (int r = 0; r < M; ++r) y = fmaf(Jc[(size_t)r * M], l[r], y);
+                for (int r = 0; r < M; ++r) y = fmaf(Jc[r * stride], l[r], y);
             }
             lds_barrier();
             if (run && ui < M) u = fmaf(rhs_sign, rhs[((size_t)ub * T + k) * M + ui], y);
@@ -287,7 +296,8 @@ __global__ __launch_bounds__(64) void k_chunk_product_dense_fwd(const float *__r
 //         coincide; per-chain max |Delta| and max |z|)
 // MODE 1: forward bare scan (y written)
 // MODE 2: reverse (y_k = J_{k+1}^T y_{k+1} + b_k written)
-template <int MP, int MODE>
+// FLIP (modes 1, 2): the other orientation of the stored matrices, as in k_chunk_product_dense
+template <int MP, int MODE, bool FLIP>
 __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J, const float *__restrict__ rhs,
                                                     float rhs_sign, const float *__restrict__ carry_in,
                                                     float *zbuf, float *outbuf, const int *__restrict__ zsel,
@@ -314,7 +324,14 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
         const int k = MODE == 2 ? s1 - 1 - t : s0 + t;
         const bool run = (MODE == 2 ? k >= s0 : k < s1) && i < M;
         const size_t e = ((size_t)b * T + k) * M + i;
-        if (MODE != 2) {
+        if ((MODE != 2) == FLIP) {
+            // column i of J_k (forward, flipped) or of J_{k+1} (reverse)
+            const int kj = MODE == 2 ? k + 1 : k;
+            const bool has = run && kj < T;
+            const float *Jc = J + ((size_t)b * T + kj) * M * M + i;
+#pragma unroll
+            for (int q = 0; q < MP; ++q) jv[q] = (has && q < M) ? Jc[(size_t)q * M] : 0.f;
+        } else if (MODE != 2) {
             const float *Jr = J + (((size_t)b * T + k) * M + i) * M;
             if ((M & 3) == 0) {   // 16-byte aligned rows: vector loads
                 const float4 *J4 = reinterpret_cast<const float4 *>(Jr);
@@ -331,10 +348,11 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
                 for (int q = 0; q < MP; ++q) jv[q] = (run && q < M) ? Jr[q] : 0.f;
             }
         } else {
+            // row i of J_{k+1} (reverse, flipped)
             const bool has = run && k + 1 < T;
-            const float *Jc = J + ((size_t)b * T + k + 1) * M * M + i;
+            const float *Jr = J + (((size_t)b * T + k + 1) * M + i) * M;
 #pragma unroll
-            for (int q = 0; q < MP; ++q) jv[q] = (has && q < M) ? Jc[(size_t)q * M] : 0.f;
+            for (int q = 0; q < MP; ++q) jv[q] = (has && q < M) ? Jr[q] : 0.f;
         }
         bv = run ? rhs[e] : 0.f;
         zv = (MODE == 0 && run) ? zin[e] : 0.f;
@@ -388,21 +406,25 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
 }
 
 int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
-                               float *P, float *v, const int *active, int C, int ncs, hipStream_t st) {
+                               float *P, float *v, const int *active, int C, int ncs, hipStream_t st, bool flip) {
     const int MP = padded_dim(M);
     const int nch = B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt("k_chunk_product_dense", st);
-#define CPD(MPV, R)                                                                                            \
-    hipLaunchKernelGGL((k_chunk_product_dense<MPV, R>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, P, v, active, \
+#define CPD(MPV, R, FL)                                                                                          \
+    hipLaunchKernelGGL((k_chunk_product_dense<MPV, R, FL>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, P, v, active, \
                        B, T, M, C, ncs)
 #define CPF(MPV)                                                                                           \
     hipLaunchKernelGGL((k_chunk_product_dense_fwd<MPV>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, P, v, \
                        active, B, T, M, C, ncs)
-    if (!rev) {
+    if (!rev && !flip) {
         if (MP == 16) CPF(16); else if (MP == 32) CPF(32); else CPF(64);
+    } else if (!rev) {
+        if (MP == 16) CPD(16, false, true); else if (MP == 32) CPD(32, false, true); else CPD(64, false, true);
+    } else if (!flip) {
+        if (MP == 16) CPD(16, true, false); else if (MP == 32) CPD(32, true, false); else CPD(64, true, false);
     } else {
-        if (MP == 16) CPD(16, true); else if (MP == 32) CPD(32, true); else CPD(64, true);
+        if (MP == 16) CPD(16, true, true); else if (MP == 32) CPD(32, true, true); else CPD(64, true, true);
     }
 #undef CPF
 #undef CPD
@@ -412,17 +434,19 @@ int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, co
 
 int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
                        const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
-                       const int *active, int C, int ncs, hipStream_t st) {
+                       const int *active, int C, int ncs, hipStream_t st, bool flip) {
     const int MP = padded_dim(M);
     const int nch = B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt(mode == 2 ? "k_fixup_dense_rev" : "k_fixup_dense_fwd", st);
-#define FXD(MPV, MO)                                                                                          \
-    hipLaunchKernelGGL((k_fixup_dense<MPV, MO>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, carry_in, z, out, \
+#define FXD(MPV, MO, FL)                                                                                          \
+    hipLaunchKernelGGL((k_fixup_dense<MPV, MO, FL>), dim3(grid), dim3(64), 0, st, J, rhs, rhs_sign, carry_in, z, out, \
                        zsel, chain_bits, active, B, T, M, C, ncs)
-#define FXD3(MO) \
-    if (MP == 16) FXD(16, MO); else if (MP == 32) FXD(32, MO); else FXD(64, MO);
-    if (mode == 0) { FXD3(0) } else if (mode == 1) { FXD3(1) } else { FXD3(2) }
+#define FXD3(MO, FL) \
+    if (MP == 16) FXD(16, MO, FL); else if (MP == 32) FXD(32, MO, FL); else FXD(64, MO, FL);
+    if (mode == 0) { FXD3(0, false) }
+    else if (mode == 1) { if (flip) { FXD3(1, true) } else { FXD3(1, false) } }
+    else { if (flip) { FXD3(2, true) } else { FXD3(2, false) } }
 #undef FXD3
 #undef FXD
     DEER_LAUNCH_CHECK("k_fixup_dense");

@@ -686,12 +686,12 @@ size_t diag_scan_ws_bytes(int B, int T, int M) {
 }
 
 int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const float *b, const float *Bc, int K,
-                     const float *u, float *y, void *ws, hipStream_t st) {
+                     const float *u, float *y, void *ws, hipStream_t st, int conj) {
     const int ntile = (M + DTC - 1) / DTC;
     const int nq = (T + DCH - 1) / DCH;
     const int nblk = B * ntile * nq;
-    const int conj_lam = rev ? 1 : 0;
-    if (!b && !rev && diag_seg_enabled()) return launch_diag_seg(B, T, M, lam, Bc, K, u, y, ws, st);
+    const int conj_lam = conj < 0 ? (rev ? 1 : 0) : (conj ? 1 : 0);
+    if (!b && !rev && conj_lam == 0 && diag_seg_enabled()) return launch_diag_seg(B, T, M, lam, Bc, K, u, y, ws, st);
     if (!diag_three_pass()) {
         const size_t nwords = (size_t)B * ntile * nq * DTC * 2;
         const size_t wbytes = (nwords * sizeof(unsigned long long) + 255) & ~(size_t)255;

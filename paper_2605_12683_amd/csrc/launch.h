@@ -146,11 +146,14 @@ int launch_qdeer_shdiag(const ShArgs &a, const uint32_t *masks, const int *activ
                         hipStream_t st);
 
 // dense stored-Jacobian scan (mode: 0 Newton fix-up, 1 bare forward scan, 2 reverse)
+// flip (bare scan only): the other orientation of every stored matrix than the direction's default
+// (forward J_t^T, reverse J_{t+1})
 int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
-                               float *P, float *v, const int *active, int C, int ncs, hipStream_t st);
+                               float *P, float *v, const int *active, int C, int ncs, hipStream_t st,
+                               bool flip = false);
 int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
                        const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
-                       const int *active, int C, int ncs, hipStream_t st);
+                       const int *active, int C, int ncs, hipStream_t st, bool flip = false);
 
 // shallow PLRNN
 size_t sh_resjac_lds(int M, int L);
@@ -178,8 +181,10 @@ int launch_readout(const RoArgs &ra, int B, int T, const float *h, const float *
 
 // diagonal complex scan
 size_t diag_scan_ws_bytes(int B, int T, int M);
+// conj < 0: the recursion multiplies by conj(lambda) when rev (the adjoint), else by lambda;
+// conj >= 0 chooses conj(lambda) (1) or lambda (0) in either direction
 int launch_diag_scan(bool rev, int B, int T, int M, const float *lam, const float *b, const float *Bc, int K,
-                     const float *u, float *y, void *ws, hipStream_t st);
+                     const float *u, float *y, void *ws, hipStream_t st, int conj = -1);
 size_t diag_adjoint_ws_bytes(int B, int T, int M, int K);
 int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const float *g, bool g_real, const float *h,
                         const float *x, float *lam_out, float *dlam, float *dBc, void *ws, hipStream_t st);

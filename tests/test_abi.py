@@ -113,3 +113,46 @@ def test_warmup_arguments(lib):
     assert st == _b.DEER_ERR_INVALID_ARG and b"tolerance" in lib.deer_last_error()
     dg = _b.deer_model(_b.DEER_DIAG_SSM, 4, 3, m.A, m.W, None, None, None)
     assert lib.deer_workspace_bytes_ex(ctypes.byref(dg), ctypes.byref(fw), 2, 64, _b.DEER_OP_SOLVE, 0) == 0
+
+
+def test_scan_workspace_query_every_orientation(lib):
+    for rev in (0, 1):
+        for tr in (0, 1):
+            assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DENSE, rev, tr, 2, 1000, 32) > 0
+            assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DIAG_C64, rev, tr, 2, 1000, 64) > 0
+    assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DENSE, 0, 0, 2, 1000, 65) == 0
+    assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DENSE, 0, 0, 0, 1000, 16) == 0
+    dummy = (ctypes.c_float * 4)()
+    p = ctypes.cast(dummy, ctypes.c_void_p)
+    st = lib.deer_scan(_b.DEER_SCAN_DENSE, 0, 1, 2, 10, 65, p, p, p, None, 0, None)
+    assert st == _b.DEER_ERR_INVALID_ARG
+    st = lib.deer_scan(_b.DEER_SCAN_DENSE, 0, 1, 2, 10, 4, p, p, p, None, 0, None)   # y aliases b
+    assert st == _b.DEER_ERR_INVALID_ARG and b"alias" in lib.deer_last_error()
+
+
+def test_solve_with_tolerance_needs_the_threads_host_block(lib):
+    """A solve with a tolerance on a thread that has not reserved its pinned host block is
+    refused before any device work (the solve itself allocates nothing)."""
+    import threading
+    m, _keep = _vanilla_model(4)
+    dummy = (ctypes.c_float * 64)()
+    p = ctypes.cast(dummy, ctypes.c_void_p)
+    out = {}
+
+    def run():
+        f = _b.deer_forcing(0.1, 2, 0)
+        o = _b.deer_solve_opts(1e-5, 10, 0, 0, 0.0)
+        out["st"] = lib.deer_solve(ctypes.byref(m), ctypes.byref(f), ctypes.byref(o), 2, 8, p, None, p, None,
+                                   None, None, p, 64, None)
+        out["msg"] = lib.deer_last_error()
+        out["q"] = lib.deer_solve_quasi(ctypes.byref(m), ctypes.byref(f), ctypes.byref(o), 2, 8, p, None, p, None,
+                                        None, None, p, 64, None)
+        out["bad"] = lib.deer_host_reserve(0)
+        out["rel"] = lib.deer_host_release()
+    t = threading.Thread(target=run)
+    t.start()
+    t.join()
+    assert out["st"] == _b.DEER_ERR_INVALID_ARG and b"deer_host_reserve" in out["msg"]
+    assert out["q"] == _b.DEER_ERR_INVALID_ARG
+    assert out["bad"] == _b.DEER_ERR_INVALID_ARG
+    assert out["rel"] == _b.DEER_OK                 # nothing to free

@@ -30,12 +30,15 @@ def _rand(B, T, M, seed):
 
 @pytest.mark.parametrize("B,T,M", [(1, 1, 1), (1, 5, 3), (2, 1023, 16), (1, 1024, 17), (3, 1025, 64),
                                    (2, 5000, 40), (1, 70000, 8)])
-@pytest.mark.parametrize("rev", [False, True])
-def test_deer_scan_diag(B, T, M, rev):
+@pytest.mark.parametrize("rev,tr", [(False, False), (True, True), (False, True), (True, False)])
+def test_deer_scan_diag(B, T, M, rev, tr):
+    """Both directions with lambda or its transpose conj(lambda) (C read as R^2)."""
     lam, b = _rand(B, T, M, B * T + M)
-    say("deer_scan diag", B, T, M, rev)
-    y = D.deer_scan(D._b.DEER_SCAN_DIAG_C64, torch.tensor(lam), torch.tensor(b), reverse=rev)
-    ref = O.diag_scan_reverse(lam, b) if rev else O.diag_scan(lam, b)
+    say("deer_scan diag", B, T, M, rev, tr)
+    y = D.deer_scan(D._b.DEER_SCAN_DIAG_C64, torch.tensor(lam), torch.tensor(b), reverse=rev, transpose=tr)
+    # the oracle's reverse scan multiplies by conj(lam); the forward one by lam
+    lop = lam if rev == tr else np.conj(lam)
+    ref = O.diag_scan_reverse(lop, b) if rev else O.diag_scan(lop, b)
     assert rel_inf(_c(y.cpu().numpy()), ref) < TOL
 
 

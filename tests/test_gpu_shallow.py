@@ -36,19 +36,22 @@ def _rand_scan(B, T, M, seed):
 
 @pytest.mark.parametrize("B,T,M,chunk", [(1, 1, 1, 0), (2, 2, 3, 0), (3, 100, 16, 0), (2, 1000, 20, 0),
                                          (1, 777, 32, 64), (2, 300, 64, 0), (2, 513, 5, 17), (1, 4000, 64, 0)])
-@pytest.mark.parametrize("rev", [False, True])
-def test_deer_scan_dense(B, T, M, chunk, rev):
-    """The bare scan y_t = J_t y_{t-1} + b_t (and its transpose) equals the sequential recurrence."""
+@pytest.mark.parametrize("rev,tr", [(False, False), (True, True), (False, True), (True, False)])
+def test_deer_scan_dense(B, T, M, chunk, rev, tr):
+    """The bare scan in both directions with each step's matrix or its transpose,
+    y_t = op(J_t) y_{t-1} + b_t or y_{t-1} = op(J_t) y_t + b_{t-1}, equals the sequential recurrence."""
     if chunk:
         os.environ["DEER_CHUNK"] = str(chunk)
     J, b = _rand_scan(B, T, M, B * T + M)
-    say("deer_scan dense", B, T, M, chunk, rev)
-    y = D.deer_scan(Bnd.DEER_SCAN_DENSE, torch.tensor(J), torch.tensor(b), reverse=rev).cpu().numpy()
+    say("deer_scan dense", B, T, M, chunk, rev, tr)
+    y = D.deer_scan(Bnd.DEER_SCAN_DENSE, torch.tensor(J), torch.tensor(b), reverse=rev, transpose=tr).cpu().numpy()
     Jd = J.astype(np.float64)
+    # the oracle's reverse recursion applies J^T; hand it J^T to get J
+    Jop = Jd if rev == tr else np.ascontiguousarray(np.swapaxes(Jd, -1, -2))
     if rev:
-        ref = O.reverse_affine_recurrence(lambda k, w: np.einsum("bi,bij->bj", w, Jd[:, k]), b.astype(np.float64))
+        ref = O.reverse_affine_recurrence(lambda k, w: np.einsum("bi,bij->bj", w, Jop[:, k]), b.astype(np.float64))
     else:
-        ref = O.affine_recurrence(lambda k, v: np.einsum("bij,bj->bi", Jd[:, k], v), b.astype(np.float64))
+        ref = O.affine_recurrence(lambda k, v: np.einsum("bij,bj->bi", Jop[:, k], v), b.astype(np.float64))
     assert rel_inf(y, ref) < TOL
 
 

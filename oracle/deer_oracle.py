@@ -20,7 +20,10 @@ Conventions (0-based arrays, paper indices in the comments):
 The observation matrix is the identity read-out of the first N latents,
 B = [I_N 0] (model-setup appendix, initialisation paragraph), so the teacher
 states are zbar_t = [x_t; 0] and the projector P_alpha = I - alpha B^+ B is
-diag(1 - a) with a_i = alpha for i < N and 0 otherwise.
+diag(1 - a) with a_i = alpha for i < N and 0 otherwise -- except in the section
+"general observation matrix" at the end, whose functions (suffix _obs) take any
+N x M matrix B, form B^+ with numpy.linalg.pinv and the dense P_alpha, and give
+the gradient with respect to B.
 
 Readings of the paper taken here (each also listed in the design notes):
   * step 1 is unforced: z~_0 := z_0 (GTF-DEER residual definition); with the
@@ -595,3 +598,243 @@ def adam_update(params: dict, grads: dict, state: dict, step: int, lr: float, be
         out[k] = np.asarray(params[k], f64) - lr * mh / (np.sqrt(vh) + eps)
         st[("m", k)], st[("v", k)] = m, v
     return out, st
+
+
+# --------------------------------------------------------------------------------------
+# general observation matrix B (N x M): dense projector and its gradient
+# (eqs. error_forcing, error_forcing_decomp; Alg. GTF-DEER: pinv(B), P_alpha, P_1, the
+# forcing targets B^+ x and the gradient g_B)
+# --------------------------------------------------------------------------------------
+
+def obs_projectors(obs: np.ndarray, alpha: float):
+    """B^+ = pinv(B), P_alpha = I - alpha B^+ B and P_1 = I - B^+ B (Alg. GTF-DEER, first line
+    of the outer loop; eq. error_forcing).  Returns (B^+ [M, N], P_alpha, P_1)."""
+    Bm = np.asarray(obs, f64)
+    Bp = np.linalg.pinv(Bm)
+    M = Bm.shape[1]
+    a = alpha_as_gpu(alpha)
+    return Bp, np.eye(M) - a * (Bp @ Bm), np.eye(M) - Bp @ Bm
+
+
+def obs_alpha_schedule(alpha: float, T: int, T_w: int = 0) -> np.ndarray:
+    """alpha_k of the forced input z~_k, k = 0..T-1: 1 in the warm-up k = 1..T_w, alpha after
+    (Alg. GTF-DEER, warm-up and forced-input lines).  Entry 0 is unused (z~_0 = z_0)."""
+    a = np.full(max(T, 1), alpha_as_gpu(alpha))
+    a[1:T_w + 1] = 1.0
+    return a
+
+
+def obs_initial_state(x: np.ndarray, obs: np.ndarray, z0=None) -> np.ndarray:
+    """z_0 = zbar_0 = B^+ x_0 unless given (Alg. GTF-DEER initialisation)."""
+    if z0 is not None:
+        return np.asarray(z0, f64).copy()
+    Bp = np.linalg.pinv(np.asarray(obs, f64))
+    return np.asarray(x, f64)[:, 0] @ Bp.T
+
+
+def obs_forced_states(z: np.ndarray, x: np.ndarray, obs: np.ndarray, alpha: float, z0=None, T_w: int = 0):
+    """z~_k = (I - alpha_k B^+ B) z_k + alpha_k B^+ x_k for k >= 1 and z~_0 = z_0 (eq.
+    error_forcing with the warm-up schedule).  z holds z_1..z_T; returns [B, T, M]."""
+    z = np.asarray(z, f64)
+    x = np.asarray(x, f64)
+    Bm = np.asarray(obs, f64)
+    Bp = np.linalg.pinv(Bm)
+    Bn, T, M = z.shape
+    ak = obs_alpha_schedule(alpha, T, T_w)
+    zt = np.zeros_like(z)
+    zt[:, 0] = obs_initial_state(x, obs, z0)
+    for k in range(1, T):
+        zk = z[:, k - 1]
+        zt[:, k] = zk - ak[k] * (zk @ (Bp @ Bm).T) + ak[k] * (x[:, k] @ Bp.T)
+    return zt
+
+
+def rollout_obs(model: dict, x: np.ndarray, obs: np.ndarray, alpha: float, z0=None, T_w: int = 0) -> np.ndarray:
+    """Sequential GTF rollout z_t = F(z~_{t-1}) with the forcing of a general observation
+    matrix (Alg. GTF-DEER's forward model; eq. error_forcing), one step at a time."""
+    model = _model64(model)
+    x = np.asarray(x, f64)
+    Bm = np.asarray(obs, f64)
+    Bp = np.linalg.pinv(Bm)
+    Bn, T1, _ = x.shape
+    T = T1 - 1
+    M = Bm.shape[1]
+    ak = obs_alpha_schedule(alpha, T, T_w)
+    zprev = obs_initial_state(x, obs, z0)
+    z = np.zeros((Bn, T, M), f64)
+    for t in range(1, T + 1):
+        k = t - 1
+        if k == 0:
+            ztil = zprev
+        else:
+            ztil = zprev - ak[k] * (zprev @ (Bp @ Bm).T) + ak[k] * (x[:, k] @ Bp.T)
+        zprev = model_map(model, ztil)
+        z[:, t - 1] = zprev
+    return z
+
+
+def newton_obs(model: dict, x: np.ndarray, obs: np.ndarray, alpha: float, *, z0=None, init: str = "teacher",
+               tol: float = 1e-5, max_iter: int = 500, fixed_iters: int = 0, T_w: int = 0, history: bool = False):
+    """GTF-DEER Newton loop (Alg. GTF-DEER) with a general observation matrix: initial guess
+    z^(0)_t = B^+ x_t, residual r_t = z_t - F(z~_{t-1}), forced Jacobians J~_t =
+    J_F(z~_{t-1}) P_{alpha_{t-1}} (eq. error_forcing_decomp; P_1 in the warm-up), the
+    update Delta_t = J~_t Delta_{t-1} - r_t by the sequential recursion, z += Delta, until
+    max |Delta| < tol per sequence (the same test as newton)."""
+    model = _model64(model)
+    x = np.asarray(x, f64)
+    Bm = np.asarray(obs, f64)
+    Bp = np.linalg.pinv(Bm)
+    Bn, T1, _ = x.shape
+    T = T1 - 1
+    M = Bm.shape[1]
+    ak = obs_alpha_schedule(alpha, T, T_w)
+    Pk = np.stack([np.eye(M) - ak[k] * (Bp @ Bm) for k in range(T)])
+    if init == "teacher":
+        z = x[:, 1:] @ Bp.T
+    elif init == "zero":
+        z = np.zeros((Bn, T, M), f64)
+    else:
+        raise ValueError(init)
+    active = np.ones(Bn, bool)
+    iters = np.zeros(Bn, np.int64)
+    norms = np.full(Bn, np.nan)
+    hist = [z.copy()] if history else None
+    k = 0
+    while True:
+        if fixed_iters > 0:
+            if k == fixed_iters:
+                break
+        elif not active.any() or k == max_iter:
+            break
+        zt = obs_forced_states(z, x, obs, alpha, z0, T_w)
+        r = z - model_map(model, zt)
+        mask = activation_mask(model, zt)
+        delta = affine_recurrence(lambda kk, v: jvp(model, mask[:, kk], v @ Pk[kk].T), -r)
+        e = np.abs(delta).reshape(Bn, -1).max(axis=1)
+        upd = active if fixed_iters == 0 else np.ones(Bn, bool)
+        z[upd] += delta[upd]
+        iters[upd] += 1
+        norms[upd] = e[upd]
+        if fixed_iters == 0:
+            active &= ~(e < tol)
+        if history:
+            hist.append(z.copy())
+        k += 1
+    out = {"z": z, "iters": iters, "norms": norms,
+           "status": "ok" if (fixed_iters > 0 or not active.any()) else "not_converged"}
+    if history:
+        out["history"] = hist
+    return out
+
+
+def mse_loss_obs(z: np.ndarray, x: np.ndarray, obs: np.ndarray, T_w: int = 0) -> float:
+    """Batch mean of (1/(N (T - T_w))) sum_{t > T_w} ||x_t - B z_t||^2 (eq. mse_loss_warmup with
+    the read-out x^_t = B z_t of eq. shplrnn_nonlinear)."""
+    z = np.asarray(z, f64)
+    x = np.asarray(x, f64)
+    Bm = np.asarray(obs, f64)
+    Bn, T, _ = z.shape
+    N = Bm.shape[0]
+    e = z[:, T_w:] @ Bm.T - x[:, 1 + T_w:]
+    return float((e ** 2).sum() / (Bn * N * (T - T_w)))
+
+
+def mse_seed_obs(z: np.ndarray, x: np.ndarray, obs: np.ndarray, T_w: int = 0) -> np.ndarray:
+    """dL/dz_t = 2/(B N (T - T_w)) B^T (B z_t - x_t) for t > T_w, zero in the warm-up."""
+    z = np.asarray(z, f64)
+    x = np.asarray(x, f64)
+    Bm = np.asarray(obs, f64)
+    Bn, T, M = z.shape
+    N = Bm.shape[0]
+    g = np.zeros((Bn, T, M), f64)
+    g[:, T_w:] = 2.0 / (Bn * N * (T - T_w)) * ((z[:, T_w:] @ Bm.T - x[:, 1 + T_w:]) @ Bm)
+    return g
+
+
+def adjoint_obs(model: dict, x: np.ndarray, z: np.ndarray, obs: np.ndarray, alpha: float, *, z0=None, g=None,
+                T_w: int = 0, mask=None) -> np.ndarray:
+    """lam = dL/dz by the backward recursion lam_T = g_T, lam_{t-1} = J~_t^T lam_t + g_{t-1}
+    with J~_t^T = P_{alpha_{t-1}}^T J_F(z~_{t-1})^T (eqs. adjoint_eq, backward_recursion).
+    mask: ReLU decisions to use instead of the float64 ones (the GPU's, for parity)."""
+    model = _model64(model)
+    z = np.asarray(z, f64)
+    Bm = np.asarray(obs, f64)
+    Bp = np.linalg.pinv(Bm)
+    M = z.shape[2]
+    ak = obs_alpha_schedule(alpha, z.shape[1], T_w)
+    Pk = np.stack([np.eye(M) - ak[k] * (Bp @ Bm) for k in range(z.shape[1])])
+    zt = obs_forced_states(z, x, obs, alpha, z0, T_w)
+    mk = activation_mask(model, zt) if mask is None else np.asarray(mask, bool)
+    g = mse_seed_obs(z, x, obs, T_w) if g is None else np.asarray(g, f64)
+    return reverse_affine_recurrence(lambda k, w: vjp(model, mk[:, k], w) @ Pk[k], g)
+
+
+def param_grads_obs(model: dict, x: np.ndarray, z: np.ndarray, obs: np.ndarray, alpha: float, lam: np.ndarray, *,
+                    z0=None, T_w: int = 0, mask=None) -> dict:
+    """dL/dtheta = sum_t lam_t^T dF(z~_{t-1})/dtheta (gradients appendix) at the forced inputs
+    of a general observation matrix; the same sums as param_grads."""
+    model = _model64(model)
+    lam = np.asarray(lam, f64)
+    zt = obs_forced_states(z, x, obs, alpha, z0, T_w)
+    mk = activation_mask(model, zt) if mask is None else np.asarray(mask, bool)
+    out = {"A": np.einsum("bti,bti->i", lam, zt, optimize=True)}
+    if model["kind"] == "plrnn":
+        out["W"] = np.einsum("bti,btj->ij", lam, np.where(mk, zt, 0.0), optimize=True)
+        out["h"] = lam.sum(axis=(0, 1))
+    else:
+        u = preactivation(model, zt)
+        delta = (lam @ _p(model, "W1")) * mk
+        out["W1"] = np.einsum("bti,btl->il", lam, np.where(mk, u, 0.0), optimize=True)
+        out["W2"] = np.einsum("btl,btj->lj", delta, zt, optimize=True)
+        out["h1"] = lam.sum(axis=(0, 1))
+        out["h2"] = delta.sum(axis=(0, 1))
+    return out
+
+
+def _dpinv_vjp(Bm: np.ndarray, Bp: np.ndarray, mu: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """Gradient with respect to B of mu^T (dB^+) v for one pair of vectors (mu in R^M, v in
+    R^N), from the differential of the Moore-Penrose inverse at constant rank (Golub and
+    Pereyra 1973): dB^+ = -B^+ dB B^+ + B^+ B^+T dB^T (I - B B^+) + (I - B^+ B) dB^T B^+T B^+.
+    Returns the N x M matrix G with mu^T (dB^+) v = sum(G * dB)."""
+    M = Bm.shape[1]
+    N = Bm.shape[0]
+    g = -np.outer(Bp.T @ mu, Bp @ v)
+    g += np.outer((np.eye(N) - Bm @ Bp) @ v, Bp @ (Bp.T @ mu))
+    g += np.outer(Bp.T @ (Bp @ v), (np.eye(M) - Bp @ Bm) @ mu)
+    return g
+
+
+def obs_grad(model: dict, x: np.ndarray, z: np.ndarray, obs: np.ndarray, alpha: float, lam: np.ndarray, *,
+             z0=None, T_w: int = 0, mask=None, with_mse: bool = True) -> np.ndarray:
+    """dL/dB (Alg. GTF-DEER, g_B of the IFT gradient): the MSE's direct term
+    2/(B N (T - T_w)) sum_{t > T_w} (B z_t - x_t) z_t^T, plus sum_t lam_t^T J_F(z~_{t-1})
+    dz~_{t-1}/dB, where z~_k = z_k + alpha_k B^+ (x_k - B z_k) for k >= 1 and, when z_0 is
+    not given, z~_0 = z_0 = B^+ x_0: with mu = J_F(z~_k)^T lam_{k+1},
+    mu^T dz~_k = alpha_k [mu^T (dB^+) e_k - mu^T B^+ dB z_k],  e_k = x_k - B z_k.
+    Each (b, k) is summed directly in float64."""
+    model = _model64(model)
+    x = np.asarray(x, f64)
+    z = np.asarray(z, f64)
+    lam = np.asarray(lam, f64)
+    Bm = np.asarray(obs, f64)
+    Bp = np.linalg.pinv(Bm)
+    Bn, T, M = z.shape
+    N = Bm.shape[0]
+    ak = obs_alpha_schedule(alpha, T, T_w)
+    zt = obs_forced_states(z, x, obs, alpha, z0, T_w)
+    mk = activation_mask(model, zt) if mask is None else np.asarray(mask, bool)
+    G = np.zeros((N, M), f64)
+    for b in range(Bn):
+        for k in range(T):
+            mu = vjp(model, mk[b, k], lam[b, k])
+            if k == 0:
+                if z0 is None:
+                    G += _dpinv_vjp(Bm, Bp, mu, x[b, 0])
+                continue
+            zk = z[b, k - 1]
+            e = x[b, k] - Bm @ zk
+            G += ak[k] * (_dpinv_vjp(Bm, Bp, mu, e) - np.outer(Bp.T @ mu, zk))
+    if with_mse:
+        e = z[:, T_w:] @ Bm.T - x[:, 1 + T_w:]
+        G += 2.0 / (Bn * N * (T - T_w)) * np.einsum("btn,btj->nj", e, z[:, T_w:])
+    return G

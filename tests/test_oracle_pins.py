@@ -771,3 +771,153 @@ def test_mar_penalty_closed_forms(kind, M, L, p):
         m["W2"][0, i] = np.float32(0.5)
         ref += c * gv / L * 0.5 ** p
     assert np.isclose(val(m), ref, rtol=1e-15, atol=0)
+
+
+# ------------------------------------------------------------------------------------
+# general observation matrix (eqs. error_forcing, error_forcing_decomp; Alg. GTF-DEER)
+# ------------------------------------------------------------------------------------
+
+def _obs(N, M, seed, scale=1.0):
+    return (np.random.default_rng(seed).standard_normal((N, M)) * scale / np.sqrt(M)).astype(np.float32)
+
+
+def test_obs_projectors_closed_forms():
+    """B = [I_N 0]: B^+ = B^T and P_alpha = diag(1 - a) (the identity read-out).  Dense B of full
+    row rank: B^+ = B^T (B B^T)^-1, P_1 is the orthogonal projector onto the null space of B
+    (P_1^2 = P_1 = P_1^T, B P_1 = 0) and P_alpha = P_1 + (1 - alpha) B^+ B; for M <= N with full
+    column rank B^+ B = I, so P_alpha = (1 - alpha) I (plain GTF)."""
+    M, N, alpha = 6, 3, 0.3
+    Bi = np.zeros((N, M), np.float32)
+    Bi[:, :N] = np.eye(N)
+    Bp, Pa, P1 = O.obs_projectors(Bi, alpha)
+    assert np.allclose(Bp, Bi.T, atol=1e-15)
+    assert np.allclose(Pa, np.diag(1.0 - O.forcing_weights(M, N, alpha)), atol=1e-15)
+    B = _obs(N, M, 5).astype(np.float64)
+    Bp, Pa, P1 = O.obs_projectors(B, alpha)
+    assert np.allclose(Bp, B.T @ np.linalg.inv(B @ B.T), atol=1e-12)
+    assert np.allclose(P1 @ P1, P1, atol=1e-12) and np.allclose(P1, P1.T, atol=1e-12)
+    assert np.allclose(B @ P1, 0.0, atol=1e-12)
+    a = O.alpha_as_gpu(alpha)
+    assert np.allclose(Pa, P1 + (1 - a) * (Bp @ B), atol=1e-12)
+    Bt = _obs(5, 4, 6).astype(np.float64)              # M = 4 <= N = 5
+    _, Pa2, _ = O.obs_projectors(Bt, alpha)
+    assert np.allclose(Pa2, (1 - a) * np.eye(4), atol=1e-12)
+
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+@pytest.mark.parametrize("T_w", [0, 9])
+def test_obs_functions_reduce_to_the_identity_readout(kind, T_w):
+    """With B = [I_N 0] every general-B function equals its identity-read-out counterpart,
+    which is pinned independently above."""
+    M, N, alpha, T = 5, 2, 0.25, 30
+    m = _vanilla(M, 91) if kind == "plrnn" else _shallow(M, 7, 92)
+    x = _x(2, T, N, 93)
+    Bi = np.zeros((N, M), np.float32)
+    Bi[:, :N] = np.eye(N)
+    z = O.rollout(m, x, alpha, N, T_w=T_w)
+    assert np.allclose(O.rollout_obs(m, x, Bi, alpha, T_w=T_w), z, rtol=1e-13, atol=1e-14)
+    assert np.allclose(O.mse_seed_obs(z, x, Bi, T_w), O.mse_seed(z, x, T_w), atol=1e-15)
+    assert abs(O.mse_loss_obs(z, x, Bi, T_w) - O.mse_loss(z, x, T_w)) < 1e-14
+    lam = O.adjoint(m, x, z, alpha, N, T_w=T_w)
+    assert np.allclose(O.adjoint_obs(m, x, z, Bi, alpha, T_w=T_w), lam, rtol=1e-12, atol=1e-15)
+    g1 = O.param_grads(m, x, z, alpha, N, lam, T_w=T_w)
+    g2 = O.param_grads_obs(m, x, z, Bi, alpha, lam, T_w=T_w)
+    for k in g1:
+        assert np.allclose(g1[k], g2[k], rtol=1e-12, atol=1e-15), k
+
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+@pytest.mark.parametrize("T_w", [0, 7])
+def test_obs_newton_converges_to_the_rollout_with_prefix_exactness(kind, T_w):
+    """Dense B (N < M): the Newton iterate reaches the sequential rollout (the unique zero of the
+    residual), and after k updates its first k states are exact (Delta_0 = 0 and the
+    block-bidiagonal structure of the forced Jacobians)."""
+    M, N, alpha, T = 5, 2, 0.3, 16
+    m = _vanilla(M, 94, w_std=0.25) if kind == "plrnn" else _shallow(M, 6, 95)
+    x = _x(2, T, N, 96)
+    B = _obs(N, M, 97)
+    ref = O.rollout_obs(m, x, B, alpha, T_w=T_w)
+    out = O.newton_obs(m, x, B, alpha, tol=1e-13, max_iter=T + 2, T_w=T_w, history=True)
+    assert out["status"] == "ok"
+    assert np.abs(out["z"] - ref).max() <= 1e-11 * max(1.0, np.abs(ref).max())
+    for k, zk in enumerate(out["history"][:T + 1]):
+        assert np.allclose(zk[:, :k], ref[:, :k], rtol=1e-10, atol=1e-11), k
+
+
+def _torch_rollout_obs(m, x, B, alpha, T_w, z0):
+    """The forward model of Alg. GTF-DEER in torch (float64), B a leaf tensor: pinv, forced
+    inputs z~ = z + a_k B^+ (x_k - B z), F, and the loss over t > T_w."""
+    Bp = torch.linalg.pinv(B)
+    X = torch.tensor(np.asarray(x, np.float64))
+    Bn, T1, _ = X.shape
+    T = T1 - 1
+    a = float(np.float32(alpha))
+    zprev = X[:, 0] @ Bp.T if z0 is None else torch.tensor(np.asarray(z0, np.float64))
+    zs = []
+    for t in range(1, T + 1):
+        k = t - 1
+        if k == 0:
+            zt = zprev
+        else:
+            ak = 1.0 if k <= T_w else a
+            zt = zprev + ak * ((X[:, k] - zprev @ B.T) @ Bp.T)
+        if m["kind"] == "plrnn":
+            zprev = m["A"] * zt + torch.relu(zt) @ m["W"].T + m["h"]
+        else:
+            zprev = m["A"] * zt + torch.relu(zt @ m["W2"].T + m["h2"]) @ m["W1"].T + m["h1"]
+        zs.append(zprev)
+    Z = torch.stack(zs, dim=1)
+    N = B.shape[0]
+    loss = ((Z[:, T_w:] @ B.T - X[:, 1 + T_w:]) ** 2).sum() / (Bn * N * (T - T_w))
+    return loss
+
+
+@pytest.mark.parametrize("kind", ["plrnn", "shplrnn"])
+@pytest.mark.parametrize("T_w,given_z0,M,N", [(0, False, 5, 2), (5, False, 5, 2), (0, True, 5, 2), (0, False, 3, 5),
+                                              (4, False, 3, 5)])
+def test_obs_gradients_match_autograd_through_the_rollout(kind, T_w, given_z0, M, N):
+    """The IFT gradients (adjoint recursion, parameter sums and dL/dB from the differential of
+    the pseudo-inverse) equal reverse-mode AD through the sequential rollout with B as a
+    parameter (torch.linalg.pinv differentiated by torch), at the rollout's fixed point.  Wide B
+    (N < M) and tall B (N > M, where B^+ B = I and the (I - B B^+) terms of the differential
+    are the ones that do not vanish)."""
+    alpha, T = 0.3, 24
+    m = _vanilla(M, 98, w_std=0.25) if kind == "plrnn" else _shallow(M, 6, 99)
+    x = _x(2, T, N, 100)
+    B = _obs(N, M, 101).astype(np.float64)
+    z0 = np.random.default_rng(102).standard_normal((2, M)) if given_z0 else None
+    z = O.rollout_obs(m, x, B, alpha, z0=z0, T_w=T_w)
+    lam = O.adjoint_obs(m, x, z, B, alpha, z0=z0, T_w=T_w)
+    gr = O.param_grads_obs(m, x, z, B, alpha, lam, z0=z0, T_w=T_w)
+    gB = O.obs_grad(m, x, z, B, alpha, lam, z0=z0, T_w=T_w)
+    P = {k: torch.tensor(np.asarray(v, np.float64), requires_grad=True) for k, v in m.items() if k != "kind"}
+    Bt = torch.tensor(B, requires_grad=True)
+    loss = _torch_rollout_obs({"kind": kind, **P}, x, Bt, alpha, T_w, z0)
+    assert abs(float(loss) - O.mse_loss_obs(z, x, B, T_w)) < 1e-13
+    loss.backward()
+    for k, v in P.items():
+        assert np.allclose(gr[k], v.grad.numpy(), rtol=1e-9, atol=1e-12), k
+    assert np.allclose(gB, Bt.grad.numpy(), rtol=1e-9, atol=1e-12)
+
+
+def test_obs_gradient_matches_central_differences():
+    """dL/dB against central differences of the loss of the rollout (float64, step 1e-6), away
+    from ReLU kinks; a second pin that does not use torch's pinv derivative."""
+    M, N, alpha, T = 4, 2, 0.35, 20
+    m = _vanilla(M, 103, w_std=0.25)
+    x = _x(1, T, N, 104)
+    B = _obs(N, M, 105).astype(np.float64)
+    z = O.rollout_obs(m, x, B, alpha)
+    lam = O.adjoint_obs(m, x, z, B, alpha)
+    gB = O.obs_grad(m, x, z, B, alpha, lam)
+    eps = 1e-6
+    fd = np.zeros_like(B)
+    for n in range(N):
+        for j in range(M):
+            Bp_, Bm_ = B.copy(), B.copy()
+            Bp_[n, j] += eps
+            Bm_[n, j] -= eps
+            lp = O.mse_loss_obs(O.rollout_obs(m, x, Bp_, alpha), x, Bp_)
+            lm = O.mse_loss_obs(O.rollout_obs(m, x, Bm_, alpha), x, Bm_)
+            fd[n, j] = (lp - lm) / (2 * eps)
+    assert np.allclose(gB, fd, rtol=1e-6, atol=1e-9)

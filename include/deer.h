@@ -44,7 +44,7 @@
  *      * the timing diagnostics (deer_timing_*), off unless enabled, which keep a
  *        mutex-protected pool of HIP events;
  *      * the read-out's resident-block count (an occupancy query made once per
- *        process).
+ *        process) and, per GPU, the scratch array of deer_scan_noalloc.
  *    Calls on different streams with different workspaces may run concurrently;
  *    calls that share a workspace must be serialised by the caller, and one host
  *    thread runs its solves one at a time.
@@ -340,6 +340,19 @@ int deer_scan(int layout, int reverse, int transpose, int B, int T, int M, const
 
 /* Workspace bytes deer_scan needs for these arguments (0 if they are invalid). */
 size_t deer_scan_workspace_bytes(int layout, int reverse, int transpose, int B, int T, int M);
+
+/* deer_scan for callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops, harnesses that forbid hipMalloc): the same scan with the same arguments and
+ * results, its scratch in a static device array of the library (deer_noalloc_scratch_bytes()
+ * = 64 MiB per GPU, held by each GPU the library runs on until the process ends) instead of a
+ * workspace.  The call allocates nothing (no hipMalloc, no events: the timing diagnostics skip
+ * it).  Sizes whose deer_scan_workspace_bytes exceeds the array are rejected with
+ * DEER_ERR_INVALID_ARG before any device work.  Every call on one GPU uses that GPU's array,
+ * which keeps the last call's contents: calls that overlap on one GPU (other streams, other
+ * threads) race and must be serialised by the caller.  Fully asynchronous on `stream`. */
+int deer_scan_noalloc(int layout, int reverse, int transpose, int B, int T, int M, const float *J,
+                      const float *b, float *y, void *stream);
+size_t deer_noalloc_scratch_bytes(void);
 
 /* Reserves the calling host thread's pinned host block for solves with a tolerance of up to
  * max_batch sequences (deer_solve, deer_solve_quasi, deer_train_step): (4 max_batch + 32)

@@ -401,3 +401,19 @@ def deer_scan(layout: int, J, b, reverse: bool = False, ws=None, transpose=None)
     _b._check(st, "deer_scan")
     return y
 
+def deer_scan_noalloc(layout: int, J, b, y, reverse: bool = False, transpose=None):
+    """deer_scan without a workspace argument: the scratch is the library's static device array
+    (deer_noalloc_scratch_bytes() bytes per GPU).  y is the caller's output buffer."""
+    lib = load()
+    J, b = _dev(J), _dev(b)
+    B, T, M = b.shape[:3]
+    tr = reverse if transpose is None else transpose
+    st = lib.deer_scan_noalloc(layout, 1 if reverse else 0, 1 if tr else 0, B, T, M, _ptr(J), _ptr(b), _ptr(y),
+                               _stream())
+    _b._check(st, "deer_scan_noalloc")
+    return y
+
+
+def deer_noalloc_scratch_bytes() -> int:
+    return int(load().deer_noalloc_scratch_bytes())
+

@@ -26,7 +26,7 @@ EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "deer_adjoint_
             "deer_last_error", "deer_timing_enable", "deer_timing_report", "deer_solve_quasi", "deer_adjoint_quasi",
             "deer_quasi_workspace_bytes", "deer_sequential", "deer_sequential_workspace_bytes",
             "deer_workspace_bytes_ex", "deer_train_step", "deer_train_workspace_bytes", "deer_train_params",
-            "deer_host_reserve", "deer_host_release"]
+            "deer_host_reserve", "deer_host_release", "deer_scan_noalloc", "deer_noalloc_scratch_bytes"]
 
 _fp = ctypes.c_void_p
 
@@ -120,6 +120,10 @@ def load(path: str = LIB_PATH):
     lib.plrnn_jacobian.restype = i32
     lib.deer_scan.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]
     lib.deer_scan.restype = i32
+    lib.deer_scan_noalloc.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp]
+    lib.deer_scan_noalloc.restype = i32
+    lib.deer_noalloc_scratch_bytes.argtypes = []
+    lib.deer_noalloc_scratch_bytes.restype = sz
     lib.deer_host_reserve.argtypes = [i32]
     lib.deer_host_reserve.restype = i32
     lib.deer_host_release.argtypes = []

@@ -33,6 +33,15 @@ int hip_fail(hipError_t e, const char *what);
 bool timing_on();
 void timing_mark(const char *name, hipStream_t st, bool start);
 
+// While one of these lives on a thread, no launch of that thread is timed (no events are made).
+void timing_suppress(bool on);
+bool timing_suppressed();
+struct TimingSuppress {
+    bool prev;
+    TimingSuppress() : prev(timing_suppressed()) { timing_suppress(true); }
+    ~TimingSuppress() { timing_suppress(prev); }
+};
+
 struct KTimer {
     const char *name;
     hipStream_t st;

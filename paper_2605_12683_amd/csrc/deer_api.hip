@@ -58,7 +58,12 @@ hipEvent_t take_event(TimingState &s) {
 }
 }  // namespace
 
+static thread_local bool t_no_timing = false;
+void timing_suppress(bool on) { t_no_timing = on; }
+bool timing_suppressed() { return t_no_timing; }
+
 bool timing_on() {
+    if (t_no_timing) return false;
     TimingState &s = tstate();
     std::lock_guard<std::mutex> g(s.mu);
     return s.on;

@@ -99,6 +99,19 @@ typedef struct {
                            the MSE seed leaves z_1..z_{T_w} out (1 / (N (T - T_w))).  PLRNN
                            kinds, solves with a tolerance (fixed_iters = 0) only; the
                            workspace is deer_workspace_bytes_ex(...).                       */
+    const float *obs;   /* general observation matrix B [n_forced, M] (device, row-major) of the
+                           read-out x^_t = B z_t, or NULL for the identity read-out B = [I_N 0].
+                           With B given (PLRNN kinds, 1 <= n_forced <= 64, n_forced may exceed
+                           M; B of full rank min(N, M)): the forcing of eq. error_forcing with
+                           the dense projector P_alpha = I - alpha B^+ B and targets B^+ x_t,
+                           J~_t = J_F(z~_{t-1}) P_alpha (eq. error_forcing_decomp), z_0 = B^+ x_0
+                           and the initial iterate B^+ x_{1:T}; the MSE seed is 2/(B N (T - T_w))
+                           B^T (B z_t - x_t); a warm-up (T_w > 0) uses P_1 = I - B^+ B and alpha = 1
+                           for z~_1..z~_{T_w} inside the same Newton iteration (Alg. GTF-DEER).
+                           B^+ and the projectors are formed on the device at the start of each
+                           call; a rank-deficient B makes them NaN (the solve then returns
+                           DEER_ERR_NONFINITE).  Supported by deer_solve and deer_adjoint(_ex);
+                           the other entry points return DEER_ERR_INVALID_ARG for it.           */
 } deer_forcing;
 
 enum { DEER_INIT_TEACHER = 0, DEER_INIT_ZERO = 1, DEER_INIT_USER = 2 };
@@ -114,16 +127,20 @@ typedef struct {
 
 /* Per-parameter gradient outputs (device, float32, NULL to skip).
  * PLRNN: A [M], W [M,M], h [M].  SHPLRNN: A [M], W [M,L] (=W1), W2 [L,M], h [M] (=h1),
- * h2 [L].  DIAG_SSM: A = dlambda [M][2], W = dBc [M,L][2] (d/dRe + i d/dIm). */
+ * h2 [L].  DIAG_SSM: A = dlambda [M][2], W = dBc [M,L][2] (d/dRe + i d/dIm).
+ * obs [N,M]: dL/dB when the forcing has an observation matrix B (Alg. GTF-DEER, g_B): the
+ * dependence of the forced inputs, of z_0 = B^+ x_0 and of the MSE on B.  With a cotangent g
+ * given instead of the MSE seed, only the first two (sum_t lam_t^T dF(z~_{t-1})/dB). */
 typedef struct {
     float *A;
     float *W;
     float *W2;
     float *h;
     float *h2;
+    float *obs;
 } deer_grads;
 
-enum { DEER_OP_SOLVE = 0, DEER_OP_ADJOINT = 1 };
+enum { DEER_OP_SOLVE = 0, DEER_OP_ADJOINT = 1, DEER_OP_JACOBIAN = 2 /* plrnn_jacobian_ex */ };
 enum { DEER_SCAN_DENSE = 0, DEER_SCAN_DIAG_C64 = 1 };
 
 /* Bytes of workspace `op` (DEER_OP_SOLVE or DEER_OP_ADJOINT) needs for this model and
@@ -135,7 +152,10 @@ size_t deer_workspace_bytes(const deer_model *model, int B, int T, int op);
  * alpha = 1, then the rest from z_0 := P_1 z_{T_w} + zbar_{T_w} -- which have the joint
  * problem's unique zero (the segments are copied through the workspace), and the adjoint as
  * the rest's adjoint followed by the prefix's, seeded with J~_{T_w+1}^T lam_{T_w+1}
- * (diag(J~_{T_w+1}) lam_{T_w+1} for quasi-DEER); the parameter gradients are summed. */
+ * (diag(J~_{T_w+1}) lam_{T_w+1} for quasi-DEER); the parameter gradients are summed.  The
+ * two solves share opts->max_iter: the rest runs at most the passes the warm-up part left (at
+ * least one), so iters reports the updates of both.  With an observation matrix
+ * (forcing->obs) the warm-up is part of the one Newton iteration instead. */
 size_t deer_workspace_bytes_ex(const deer_model *model, const deer_forcing *forcing, int B, int T, int op,
                                int quasi);
 
@@ -318,6 +338,15 @@ int deer_readout_loss(const deer_readout *readout, int B, int T, int M, const fl
 int plrnn_jacobian(const deer_model *model, const deer_forcing *forcing, int B, int T,
                    const float *x, const float *z0, const float *z, float *F, float *r, float *J,
                    uint32_t *masks, void *stream);
+
+/* plrnn_jacobian for any forcing: with forcing->obs (a general observation matrix; a warm-up
+ * T_w > 0 allowed) the residual, masks and forced Jacobians of that forcing, computed by the
+ * same kernels deer_solve and deer_adjoint use (so the masks are the decisions they take), with
+ * deer_workspace_bytes_ex(model, forcing, B, T, DEER_OP_JACOBIAN, 0) bytes of workspace; without
+ * obs it is plrnn_jacobian (ws unused).  Fully asynchronous. */
+int plrnn_jacobian_ex(const deer_model *model, const deer_forcing *forcing, int B, int T,
+                      const float *x, const float *z0, const float *z, float *F, float *r, float *J,
+                      uint32_t *masks, void *ws, size_t ws_bytes, void *stream);
 
 /* The bare associative scan over affine pairs (scheduled-sampling appendix: the pair
  * (A_t, b_t) and its composition), batched over B independent sequences of length T.

@@ -161,13 +161,14 @@ def _workspace(nbytes: int):
 
 def deer_solve(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1e-5, max_iter: int = 500,
                fixed_iters: int = 0, init: str = "teacher", z=None, want_masks: bool = False, ws=None,
-               check: bool = True, step_bound: float = 0.0, T_w: int = 0) -> dict:
+               check: bool = True, step_bound: float = 0.0, T_w: int = 0, obs=None) -> dict:
     """GTF-DEER forward solve.  Returns dict(z, masks, iters, norms, status).  step_bound:
     threshold of the update safeguard (0: library default, < 0: only non-finite updates are
-    rejected).  T_w: latent warm-up steps."""
+    rejected).  T_w: latent warm-up steps.  obs: observation matrix B [N, M] (N = n_forced) of
+    the read-out x^ = B z, or None for the identity read-out of the first n_forced latents."""
     return _solve("deer_solve", 0, model, x, alpha, n_forced, z0=z0, tol=tol, max_iter=max_iter,
                   fixed_iters=fixed_iters, init=init, z=z, want_masks=want_masks, ws=ws, check=check,
-                  step_bound=step_bound, T_w=T_w)
+                  step_bound=step_bound, T_w=T_w, obs=obs)
 
 
 def deer_solve_quasi(model, x, alpha: float, n_forced: int, *, z0=None, tol: float = 1e-5, max_iter: int = 500,
@@ -181,7 +182,7 @@ def deer_solve_quasi(model, x, alpha: float, n_forced: int, *, z0=None, tol: flo
 
 
 def _solve(entry, quasi, model, x, alpha, n_forced, *, z0, tol, max_iter, fixed_iters, init, z, want_masks, ws,
-           check, step_bound, T_w):
+           check, step_bound, T_w, obs=None):
     lib = load()
     m = _model(model)
     x = _dev(x)
@@ -197,7 +198,8 @@ def _solve(entry, quasi, model, x, alpha, n_forced, *, z0, tol, max_iter, fixed_
     if want_masks:
         H = m.M if m.kind == "plrnn" else m.L
         masks = torch.empty(B, T, (H + 31) // 32, dtype=torch.int32, device="cuda")
-    f = _b.deer_forcing(float(alpha), int(n_forced), int(T_w))
+    obsd = _dev(obs)
+    f = _b.deer_forcing(float(alpha), int(n_forced), int(T_w), _ptr(obsd))
     if ws is None:
         ws = _workspace(lib.deer_workspace_bytes_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _b.DEER_OP_SOLVE, quasi))
     iters = (ctypes.c_int32 * B)()
@@ -215,10 +217,11 @@ def _solve(entry, quasi, model, x, alpha, n_forced, *, z0, tol, max_iter, fixed_
 
 
 def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, want_lam: bool = True,
-                 want_grads: bool = True, ws=None, T_w: int = 0) -> dict:
+                 want_grads: bool = True, ws=None, T_w: int = 0, obs=None) -> dict:
     """Adjoint scan lam = dL/dz and parameter gradients at trajectory z.  Diagonal SSM: g is
     complex [B,T,M] (or [B,T,M,2] float) = dL/dRe h + i dL/dIm h, or a real float tensor
-    [B,T,M] = dL/dRe h (the read-out's cotangent)."""
+    [B,T,M] = dL/dRe h (the read-out's cotangent).  obs: observation matrix B [N, M] as in
+    deer_solve; the gradients then include "obs" = dL/dB."""
     lib = load()
     m = _model(model)
     x = _dev(x)
@@ -249,7 +252,11 @@ def deer_adjoint(model, x, z, alpha: float, n_forced: int, *, z0=None, g=None, w
         else:
             grads = {"lam": torch.empty(m.M, 2, device="cuda"), "Bc": torch.empty(m.M, m.L, 2, device="cuda")}
             gs = _b.deer_grads(_ptr(grads["lam"]), _ptr(grads["Bc"]), None, None, None)
-    f = _b.deer_forcing(float(alpha), int(n_forced), int(T_w))
+    obsd = _dev(obs)
+    if want_grads and obsd is not None:
+        grads["obs"] = torch.empty(obsd.shape, device="cuda")
+        gs.obs = _ptr(grads["obs"])
+    f = _b.deer_forcing(float(alpha), int(n_forced), int(T_w), _ptr(obsd))
     if ws is None:
         ws = _workspace(lib.deer_workspace_bytes_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _b.DEER_OP_ADJOINT, 0))
     z0d = _dev(z0)
@@ -363,8 +370,9 @@ def deer_sequential_workspace_bytes(model, B: int, T: int) -> int:
 
 
 def plrnn_jacobian(model, x, z, alpha: float, n_forced: int, *, z0=None, want=("F", "r", "masks"),
-                   dense_J: bool = False) -> dict:
-    """F, r, masks (and optionally the dense forced Jacobians) at trajectory z."""
+                   dense_J: bool = False, obs=None, T_w: int = 0) -> dict:
+    """F, r, masks (and optionally the dense forced Jacobians) at trajectory z.  obs / T_w: an
+    observation matrix B [N, M] and a warm-up (plrnn_jacobian_ex in the C ABI)."""
     lib = load()
     m = _model(model)
     x = _dev(x)
@@ -376,10 +384,16 @@ def plrnn_jacobian(model, x, z, alpha: float, n_forced: int, *, z0=None, want=("
     r = torch.empty(B, T, M, device="cuda") if "r" in want else None
     J = torch.empty(B, T, M, M, device="cuda") if dense_J else None
     masks = torch.empty(B, T, (H + 31) // 32, dtype=torch.int32, device="cuda") if "masks" in want else None
-    f = _b.deer_forcing(float(alpha), int(n_forced))
+    obsd = _dev(obs)
+    f = _b.deer_forcing(float(alpha), int(n_forced), int(T_w), _ptr(obsd))
     z0d = _dev(z0)
-    st = lib.plrnn_jacobian(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(F), _ptr(r),
-                            _ptr(J), _ptr(masks), _stream())
+    if obsd is None and T_w == 0:
+        st = lib.plrnn_jacobian(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(F),
+                                _ptr(r), _ptr(J), _ptr(masks), _stream())
+    else:
+        ws = _workspace(lib.deer_workspace_bytes_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _b.DEER_OP_JACOBIAN, 0))
+        st = lib.plrnn_jacobian_ex(ctypes.byref(m.c), ctypes.byref(f), B, T, _ptr(x), _ptr(z0d), _ptr(z), _ptr(F),
+                                   _ptr(r), _ptr(J), _ptr(masks), _ptr(ws), ws.numel(), _stream())
     _b._check(st, "plrnn_jacobian")
     out.update({"F": F, "r": r, "J": J, "masks": masks})
     return out

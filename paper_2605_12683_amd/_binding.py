@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libdeer.so")
 DEER_OK, DEER_ERR_INVALID_ARG, DEER_ERR_NOT_CONVERGED, DEER_ERR_NONFINITE, DEER_ERR_HIP, DEER_ERR_WORKSPACE = range(6)
 DEER_PLRNN, DEER_SHPLRNN, DEER_DIAG_SSM = 0, 1, 2
 DEER_INIT_TEACHER, DEER_INIT_ZERO, DEER_INIT_USER = 0, 1, 2
-DEER_OP_SOLVE, DEER_OP_ADJOINT = 0, 1
+DEER_OP_SOLVE, DEER_OP_ADJOINT, DEER_OP_JACOBIAN = 0, 1, 2
 DEER_SCAN_DENSE, DEER_SCAN_DIAG_C64 = 0, 1
 DEER_G_NATIVE, DEER_G_REAL = 0, 1
 
@@ -26,7 +26,8 @@ EXPORTED = ["deer_workspace_bytes", "deer_solve", "deer_adjoint", "deer_adjoint_
             "deer_last_error", "deer_timing_enable", "deer_timing_report", "deer_solve_quasi", "deer_adjoint_quasi",
             "deer_quasi_workspace_bytes", "deer_sequential", "deer_sequential_workspace_bytes",
             "deer_workspace_bytes_ex", "deer_train_step", "deer_train_workspace_bytes", "deer_train_params",
-            "deer_host_reserve", "deer_host_release", "deer_scan_noalloc", "deer_noalloc_scratch_bytes"]
+            "deer_host_reserve", "deer_host_release", "deer_scan_noalloc", "deer_noalloc_scratch_bytes",
+            "plrnn_jacobian_ex"]
 
 _fp = ctypes.c_void_p
 
@@ -44,7 +45,7 @@ class deer_train_opts(ctypes.Structure):
 
 
 class deer_forcing(ctypes.Structure):
-    _fields_ = [("alpha", ctypes.c_float), ("n_forced", ctypes.c_int), ("T_w", ctypes.c_int)]
+    _fields_ = [("alpha", ctypes.c_float), ("n_forced", ctypes.c_int), ("T_w", ctypes.c_int), ("obs", _fp)]
 
 
 class deer_solve_opts(ctypes.Structure):
@@ -53,7 +54,7 @@ class deer_solve_opts(ctypes.Structure):
 
 
 class deer_grads(ctypes.Structure):
-    _fields_ = [("A", _fp), ("W", _fp), ("W2", _fp), ("h", _fp), ("h2", _fp)]
+    _fields_ = [("A", _fp), ("W", _fp), ("W2", _fp), ("h", _fp), ("h2", _fp), ("obs", _fp)]
 
 
 class deer_readout(ctypes.Structure):
@@ -118,6 +119,8 @@ def load(path: str = LIB_PATH):
     lib.deer_readout_loss.restype = i32
     lib.plrnn_jacobian.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.plrnn_jacobian.restype = i32
+    lib.plrnn_jacobian_ex.argtypes = [P(deer_model), P(deer_forcing), i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.plrnn_jacobian_ex.restype = i32
     lib.deer_scan.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]
     lib.deer_scan.restype = i32
     lib.deer_scan_noalloc.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp]

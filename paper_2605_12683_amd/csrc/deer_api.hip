@@ -512,7 +512,15 @@ static int check_common(const deer_model *m, const deer_forcing *f, int B, int T
     if (m->M <= 0) { set_error("M must be positive"); return DEER_ERR_INVALID_ARG; }
     if (m->kind == DEER_PLRNN || m->kind == DEER_SHPLRNN) {
         if (m->M > 64) { set_error("M=%d unsupported (dense scans support M <= 64)", m->M); return DEER_ERR_INVALID_ARG; }
-        if (f->n_forced < 0 || f->n_forced > m->M) { set_error("n_forced must lie in [0, M]"); return DEER_ERR_INVALID_ARG; }
+        if (f->obs) {
+            if (f->n_forced < 1 || f->n_forced > 64) {
+                set_error("with an observation matrix, n_forced (its row count) must lie in [1, 64]");
+                return DEER_ERR_INVALID_ARG;
+            }
+        } else if (f->n_forced < 0 || f->n_forced > m->M) {
+            set_error("n_forced must lie in [0, M]");
+            return DEER_ERR_INVALID_ARG;
+        }
         if (!m->A || !m->W) { set_error("model parameters A and W are required"); return DEER_ERR_INVALID_ARG; }
         if (m->kind == DEER_SHPLRNN) {
             if (m->L <= 0 || m->L > 1024 || !m->W2) { set_error("shallow PLRNN needs W2 and 1 <= L <= 1024"); return DEER_ERR_INVALID_ARG; }
@@ -533,12 +541,26 @@ static int check_common(const deer_model *m, const deer_forcing *f, int B, int T
         set_error("the latent warm-up applies to the PLRNN kinds");
         return DEER_ERR_INVALID_ARG;
     }
+    if (f->obs && m->kind == DEER_DIAG_SSM) {
+        set_error("an observation matrix applies to the PLRNN kinds");
+        return DEER_ERR_INVALID_ARG;
+    }
+    return DEER_OK;
+}
+
+// entry points that take the identity read-out only
+static int no_obs(const deer_forcing *f, const char *entry) {
+    if (f && f->obs) {
+        set_error("%s: a general observation matrix is supported by deer_solve and deer_adjoint only", entry);
+        return DEER_ERR_INVALID_ARG;
+    }
     return DEER_OK;
 }
 
 static int check_quasi(const deer_model *m, const deer_forcing *f, int B, int T) {
     int rc = check_common(m, f, B, T);
     if (rc) return rc;
+    if ((rc = no_obs(f, "quasi-DEER"))) return rc;
     if (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN) {
         set_error("quasi-DEER is built for the PLRNN kinds only");
         return DEER_ERR_INVALID_ARG;
@@ -899,6 +921,209 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
     return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
 }
 
+// ---- general observation matrix (eq. error_forcing with a dense P_alpha; Alg. GTF-DEER) ----------
+// The forcing is formed by k_obs_forced (z~_s = P_s z + alpha_s B^+ x_s, P_1 in the warm-up) into a
+// forced-input array that the stored-Jacobian kernels read in place of their own diagonal forcing;
+// the vanilla PLRNN runs through them as the shallow form with W2 = I, h2 = 0 (u = z~ exactly, so
+// its ReLU decisions are those of z~).  J~_s = diag(A) P_s + W1 diag(m) (W2 P_s) is formed per step
+// range (P_1 for s <= T_w, P_alpha after), then the dense scan solves the update; the warm-up is
+// part of the one Newton iteration.
+struct ObsWs {
+    double *Bp64, *B64, *P164, *bgrad, *aug;
+    float *Bp32, *Pa32, *P132, *Ca, *C1, *Id, *Va, *V1;
+    float *Zt, *z0e;
+    ShWs sh;
+};
+
+static ObsWs carve_obs(void *ws, const deer_model *m, const deer_forcing *f, int B, int T, int op, size_t *bytes) {
+    const int M = m->M, N = f->n_forced, L = m->kind == DEER_SHPLRNN ? m->L : M;
+    ObsWs w{};
+    Carver c(ws);
+    w.Bp64 = c.take<double>((size_t)M * N);
+    w.B64 = c.take<double>((size_t)N * M);
+    w.P164 = c.take<double>((size_t)M * M);
+    w.aug = c.take<double>((size_t)64 * 128);
+    w.Bp32 = c.take<float>((size_t)M * N);
+    w.Pa32 = c.take<float>((size_t)M * M);
+    w.P132 = c.take<float>((size_t)M * M);
+    w.Ca = c.take<float>((size_t)M * M);
+    w.C1 = c.take<float>((size_t)M * M);
+    w.Id = c.take<float>((size_t)M * M);
+    w.Va = c.take<float>((size_t)L * M);
+    w.V1 = c.take<float>((size_t)L * M);
+    w.Zt = c.take<float>((size_t)B * T * M);
+    w.z0e = c.take<float>((size_t)B * M);
+    if (op == DEER_OP_ADJOINT) w.bgrad = c.take<double>(obs_bgrad_ws_doubles(M, N));
+    if (op == DEER_OP_JACOBIAN) {
+        w.sh.masks = c.take<uint32_t>((size_t)B * T * ((L + 31) / 32));
+        *bytes = c.off;
+        return w;
+    }
+    size_t shb = 0;
+    w.sh = carve_sh(ws ? (char *)ws + c.off : nullptr, B, T, M, L, op, true, true, &shb);
+    *bytes = c.off + shb;
+    return w;
+}
+
+static int obs_prepare(const deer_model *m, const deer_forcing *f, const ObsWs &w, hipStream_t st) {
+    const bool sh = m->kind == DEER_SHPLRNN;
+    ObsSetup s{f->obs, f->n_forced, m->M, sh ? m->L : m->M, f->alpha, m->A, sh ? m->W2 : nullptr,
+               w.Bp64, w.B64, w.P164, w.Bp32, w.Pa32, w.P132, w.Ca, w.C1, w.Id, w.Va, w.V1, w.aug};
+    return launch_obs_setup(s, st);
+}
+
+// J~ of every step into J: P_1 for the warm-up steps s = 0..T_w (step 0's Jacobian only multiplies
+// Delta_0 = 0), P_alpha after; plain J_F (P = I) when unforced is set
+static int obs_jacform(const deer_model *m, const deer_forcing *f, const ObsWs &w, int B, int T, const float *x,
+                       const float *z0e, const uint32_t *masks, float *J, const int *active, const float *gamma,
+                       bool unforced, hipStream_t st) {
+    const bool sh = m->kind == DEER_SHPLRNN;
+    const int L = sh ? m->L : m->M;
+    ShArgs a{m->A, m->W, nullptr, m->h, sh ? m->h2 : nullptr, 0.f, 0, x, z0e, B, T, m->M, L};
+    if (unforced) {
+        a.W2 = sh ? m->W2 : w.Id;
+        return launch_jacform_shplrnn(a, masks, J, active, gamma, st);
+    }
+    int rc;
+    if (f->T_w > 0) {
+        a.W2 = w.V1;
+        a.Cd = w.C1;
+        a.t_lo = 0;
+        a.t_hi = f->T_w + 1;
+        if ((rc = launch_jacform_shplrnn(a, masks, J, active, gamma, st))) return rc;
+        if (f->T_w + 1 >= T) return DEER_OK;
+        a.t_lo = f->T_w + 1;
+        a.t_hi = T;
+    }
+    a.W2 = w.Va;
+    a.Cd = w.Ca;
+    return launch_jacform_shplrnn(a, masks, J, active, gamma, st);
+}
+
+static int solve_obs(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
+                     const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
+                     void *ws, size_t ws_bytes, hipStream_t st) {
+    int rc;
+    const bool sh = m->kind == DEER_SHPLRNN;
+    if (sh && (rc = check_shallow_limits(m))) return rc;
+    const int M = m->M, N = f->n_forced, L = sh ? m->L : M;
+    size_t need = 0;
+    carve_obs(nullptr, m, f, B, T, DEER_OP_SOLVE, &need);
+    if ((rc = check_ws(ws, ws_bytes, need))) return rc;
+    ObsWs w = carve_obs(ws, m, f, B, T, DEER_OP_SOLVE, &need);
+    if ((rc = obs_prepare(m, f, w, st))) return rc;
+    if (o->init == DEER_INIT_TEACHER) {
+        if ((rc = launch_obs_forced(1, nullptr, nullptr, nullptr, x, z0, w.Bp32, w.Pa32, w.P132, f->alpha, f->T_w, B, T,
+                                    M, N, z, w.z0e, st)))
+            return rc;
+    } else if (o->init == DEER_INIT_ZERO) {
+        if ((rc = launch_fill_f32(z, (size_t)B * T * M, 0.f, st))) return rc;
+    }
+    const float *z0e = z0 ? z0 : w.z0e;
+    ShArgs ar{m->A, m->W, sh ? m->W2 : w.Id, m->h, sh ? m->h2 : nullptr, 0.f, 0, x, z0e, B, T, M, L};
+    ar.zt = w.Zt;
+    std::vector<int> act(B, 1), it(B, 0);
+    std::vector<float> norm(B, NAN);
+    bool nonfinite = false;
+    const ShWs &s = w.sh;
+    const DenseWs &d = s.d;
+    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *,
+                      uint32_t) -> int {
+        int r;
+        if ((r = launch_obs_forced(0, zb, za, zsel, x, z0, w.Bp32, w.Pa32, w.P132, f->alpha, f->T_w, B, T, M, N, w.Zt,
+                                   w.z0e, st)))
+            return r;
+        if ((r = launch_resjac_shplrnn(ar, zb, za, zsel, nullptr, s.r, s.masks, dact, st))) return r;
+        if ((r = obs_jacform(m, f, w, B, T, x, z0e, s.masks, s.J, dact, gam, false, st))) return r;
+        if ((r = launch_chunk_product_dense(false, B, T, M, s.J, s.r, -1.f, d.P, d.v, dact, d.C, d.ncs, st))) return r;
+        if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nullptr, B, d.ncs, d.gws, st))) return r;
+        return launch_fixup_dense(0, B, T, M, s.J, s.r, -1.f, d.carry, zb, za, zsel, s.ctl.chain_bits, dact, d.C,
+                                  d.ncs, st);
+    };
+    if ((rc = newton_loop(o, B, (size_t)T * M, d.ncs, s.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
+    if (masks) {
+        if ((rc = launch_obs_forced(0, z, nullptr, nullptr, x, z0, w.Bp32, w.Pa32, w.P132, f->alpha, f->T_w, B, T, M,
+                                    N, w.Zt, w.z0e, st)))
+            return rc;
+        if ((rc = launch_resjac_shplrnn(ar, z, nullptr, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
+    }
+    return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
+}
+
+static int jacobian_obs(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
+                        const float *z, float *F, float *r, float *J, uint32_t *masks, void *ws, size_t ws_bytes,
+                        hipStream_t st) {
+    int rc;
+    const bool sh = m->kind == DEER_SHPLRNN;
+    if (sh && (rc = check_shallow_limits(m))) return rc;
+    const int M = m->M, N = f->n_forced, L = sh ? m->L : M;
+    size_t need = 0;
+    carve_obs(nullptr, m, f, B, T, DEER_OP_JACOBIAN, &need);
+    if ((rc = check_ws(ws, ws_bytes, need))) return rc;
+    ObsWs w = carve_obs(ws, m, f, B, T, DEER_OP_JACOBIAN, &need);
+    if ((rc = obs_prepare(m, f, w, st))) return rc;
+    if ((rc = launch_obs_forced(0, z, nullptr, nullptr, x, z0, w.Bp32, w.Pa32, w.P132, f->alpha, f->T_w, B, T, M, N,
+                                w.Zt, w.z0e, st)))
+        return rc;
+    const float *z0e = z0 ? z0 : w.z0e;
+    ShArgs ar{m->A, m->W, sh ? m->W2 : w.Id, m->h, sh ? m->h2 : nullptr, 0.f, 0, x, z0e, B, T, M, L};
+    ar.zt = w.Zt;
+    uint32_t *mk = masks ? masks : w.sh.masks;
+    if ((rc = launch_resjac_shplrnn(ar, z, nullptr, nullptr, F, r, mk, nullptr, st))) return rc;
+    if (J) return obs_jacform(m, f, w, B, T, x, z0e, mk, J, nullptr, nullptr, false, st);
+    return DEER_OK;
+}
+
+static int adjoint_obs(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
+                       const float *z, const float *g, float *lam, const deer_grads *grads, void *ws, size_t ws_bytes,
+                       hipStream_t st) {
+    int rc;
+    const bool sh = m->kind == DEER_SHPLRNN;
+    if (sh && (rc = check_shallow_limits(m))) return rc;
+    const int M = m->M, N = f->n_forced, L = sh ? m->L : M;
+    size_t need = 0;
+    carve_obs(nullptr, m, f, B, T, DEER_OP_ADJOINT, &need);
+    if ((rc = check_ws(ws, ws_bytes, need))) return rc;
+    ObsWs w = carve_obs(ws, m, f, B, T, DEER_OP_ADJOINT, &need);
+    const ShWs &s = w.sh;
+    const DenseWs &d = s.d;
+    if ((rc = obs_prepare(m, f, w, st))) return rc;
+    if ((rc = launch_obs_forced(0, z, nullptr, nullptr, x, z0, w.Bp32, w.Pa32, w.P132, f->alpha, f->T_w, B, T, M, N,
+                                w.Zt, w.z0e, st)))
+        return rc;
+    const float *z0e = z0 ? z0 : w.z0e;
+    ShArgs ar{m->A, m->W, sh ? m->W2 : w.Id, m->h, sh ? m->h2 : nullptr, 0.f, 0, x, z0e, B, T, M, L};
+    ar.zt = w.Zt;
+    if ((rc = launch_resjac_shplrnn(ar, z, nullptr, nullptr, nullptr, nullptr, s.masks, nullptr, st))) return rc;
+    if ((rc = obs_jacform(m, f, w, B, T, x, z0e, s.masks, s.J, nullptr, nullptr, false, st))) return rc;
+    const double mse_scale = 2.0 / ((double)B * N * (T - f->T_w));
+    const float *gg = g;
+    if (!gg) {
+        if ((rc = launch_obs_seed(z, x, f->obs, (float)mse_scale, f->T_w, B, T, M, N, s.g, st))) return rc;
+        gg = s.g;
+    }
+    float *lo = lam ? lam : s.lam;
+    if ((rc = launch_chunk_product_dense(true, B, T, M, s.J, gg, 1.f, d.P, d.v, nullptr, d.C, d.ncs, st))) return rc;
+    if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, d.gws, st))) return rc;
+    if ((rc = launch_fixup_dense(2, B, T, M, s.J, gg, 1.f, d.carry, nullptr, lo, nullptr, nullptr, nullptr, d.C, d.ncs,
+                                 st)))
+        return rc;
+    if (!grads) return DEER_OK;
+    if (grads->A || grads->W || grads->W2 || grads->h || grads->h2) {
+        // the vanilla PLRNN as the shallow form: dW1 is dW, dh1 is dh, W2 = I and h2 are not parameters
+        deer_grads gv{grads->A, grads->W, sh ? grads->W2 : nullptr, grads->h, sh ? grads->h2 : nullptr, nullptr};
+        if ((rc = launch_grads_shplrnn(ar, z, lo, s.masks, s.part, &gv, st))) return rc;
+    }
+    if (grads->obs) {
+        // mu_s = J_F(z~_s)^T lam_s needs the unforced Jacobians: formed into J (J~ is no longer used)
+        if ((rc = obs_jacform(m, f, w, B, T, x, z0e, s.masks, s.J, nullptr, nullptr, true, st))) return rc;
+        if ((rc = launch_obs_bgrad(s.J, lo, z, x, f->obs, w.Bp64, w.B64, w.P164, z0 != nullptr, f->alpha, f->T_w,
+                                   g == nullptr, mse_scale, B, T, M, N, w.bgrad, grads->obs, st)))
+            return rc;
+    }
+    return DEER_OK;
+}
+
 static int solve_quasi(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
                        const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
                        void *ws, size_t ws_bytes, hipStream_t st) {
@@ -1027,7 +1252,16 @@ static int solve_warmup(const deer_model *m, const deer_forcing *f, const deer_s
     if (r1 != DEER_OK && r1 != DEER_ERR_NOT_CONVERGED && r1 != DEER_ERR_NONFINITE) return r1;
     hipLaunchKernelGGL(k_warmup_state, dim3(B), dim3(64), 0, st, x, (const float *)w.z1, w.zb, T, T1, M, N);
     DEER_LAUNCH_CHECK("k_warmup_state");
-    const int r2 = solve(m, &f2, o, B, T2, w.x2, w.zb, w.z2, masks ? w.m2 : nullptr, it2.data(), n2.data(), w.inner,
+    // the two parts share the pass budget: the rest gets what the warm-up part left (at least one
+    // pass); a pass is an accepted or rejected update, so the warm-up part took at least max it1
+    deer_solve_opts o2 = *o;
+    {
+        const int cap = o->max_iter > 0 ? o->max_iter : 500;
+        int used = 0;
+        for (int b = 0; b < B; ++b) used = it1[b] > used ? it1[b] : used;
+        o2.max_iter = cap - used > 1 ? cap - used : 1;
+    }
+    const int r2 = solve(m, &f2, &o2, B, T2, w.x2, w.zb, w.z2, masks ? w.m2 : nullptr, it2.data(), n2.data(), w.inner,
                          w.inner_bytes, st);
     if (r2 != DEER_OK && r2 != DEER_ERR_NOT_CONVERGED && r2 != DEER_ERR_NONFINITE) return r2;
     if ((rc = copy_rows(z, w.z1, B, T1, M, T1, 0, T, 0, st))) return rc;
@@ -1214,12 +1448,28 @@ size_t deer_scan_workspace_bytes(int layout, int reverse, int transpose, int B, 
     return 0;
 }
 
+int plrnn_jacobian_ex(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
+                      const float *z, float *F, float *r, float *J, uint32_t *masks, void *ws, size_t ws_bytes,
+                      void *stream) {
+    set_error("");
+    int rc = check_common(m, f, B, T);
+    if (rc) return rc;
+    if (!f->obs) return plrnn_jacobian(m, f, B, T, x, z0, z, F, r, J, masks, stream);
+    if (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN) {
+        set_error("plrnn_jacobian_ex: PLRNN kinds only");
+        return DEER_ERR_INVALID_ARG;
+    }
+    if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
+    return jacobian_obs(m, f, B, T, x, z0, z, F, r, J, masks, ws, ws_bytes, (hipStream_t)stream);
+}
+
 int plrnn_jacobian(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
                    const float *z, float *F, float *r, float *J, uint32_t *masks, void *stream) {
     set_error("");
     int rc = check_common(m, f, B, T);
     if (rc) return rc;
     if (f->T_w != 0) { set_error("plrnn_jacobian takes T_w = 0 (one forcing strength for every step)"); return DEER_ERR_INVALID_ARG; }
+    if ((rc = no_obs(f, "plrnn_jacobian"))) return rc;
     if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
     hipStream_t st = (hipStream_t)stream;
     if (m->kind == DEER_PLRNN) {
@@ -1251,6 +1501,7 @@ int deer_solve(const deer_model *m, const deer_forcing *f, const deer_solve_opts
     if (!(o->tol >= 0.f) && o->fixed_iters <= 0) { set_error("tol must be >= 0"); return DEER_ERR_INVALID_ARG; }
     if (m->kind != DEER_DIAG_SSM && o->fixed_iters <= 0 && (rc = check_host_reserved(B))) return rc;
     hipStream_t st = (hipStream_t)stream;
+    if (f->obs) return solve_obs(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
     if (f->T_w > 0) return solve_warmup(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st, false);
     if (m->kind == DEER_PLRNN)
         return solve_plrnn(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
@@ -1290,6 +1541,7 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
     if (rc) return rc;
     if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
     hipStream_t st = (hipStream_t)stream;
+    if (f->obs) return adjoint_obs(m, f, B, T, x, z0, z, g, lam, grads, ws, ws_bytes, st);
     if (f->T_w > 0) {
         if (g_layout != DEER_G_NATIVE) { set_error("the latent warm-up takes the native cotangent layout"); return DEER_ERR_INVALID_ARG; }
         return adjoint_warmup(m, f, B, T, x, z0, z, g, lam, grads, ws, ws_bytes, st, false);
@@ -1417,6 +1669,14 @@ int deer_adjoint_quasi(const deer_model *m, const deer_forcing *f, int B, int T,
 }
 
 size_t deer_workspace_bytes_ex(const deer_model *m, const deer_forcing *f, int B, int T, int op, int quasi) {
+    if (f && f->obs) {
+        if (quasi || check_common(m, f, B, T) != DEER_OK) return 0;
+        if (op != DEER_OP_SOLVE && op != DEER_OP_ADJOINT && op != DEER_OP_JACOBIAN) return 0;
+        if (m->kind == DEER_SHPLRNN && check_shallow_limits(m) != DEER_OK) return 0;
+        size_t bytes = 0;
+        carve_obs(nullptr, m, f, B, T, op, &bytes);
+        return bytes;
+    }
     if (!f || f->T_w == 0) return quasi ? deer_quasi_workspace_bytes(m, B, T, op) : deer_workspace_bytes(m, B, T, op);
     if ((quasi ? check_quasi(m, f, B, T) : check_common(m, f, B, T)) != DEER_OK) return 0;
     if (op != DEER_OP_SOLVE && op != DEER_OP_ADJOINT) return 0;
@@ -1451,6 +1711,7 @@ int deer_train_step(const deer_model *m, const deer_forcing *f, const deer_solve
     if (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN) { set_error("deer_train_step: PLRNN kinds only"); return DEER_ERR_INVALID_ARG; }
     if (!o || !tr || !x || !z || !adam_m || !adam_v) { set_error("opts, train, x, z and the Adam moments are required"); return DEER_ERR_INVALID_ARG; }
     if (o->fixed_iters > 0) { set_error("deer_train_step solves to a tolerance (fixed_iters = 0)"); return DEER_ERR_INVALID_ARG; }
+    if ((rc = no_obs(f, "deer_train_step"))) return rc;
     if ((rc = check_host_reserved(B))) return rc;
     if (tr->step < 1 || !(tr->lr > 0.f) || !(tr->beta1 >= 0.f && tr->beta1 < 1.f) || !(tr->beta2 >= 0.f && tr->beta2 < 1.f)) {
         set_error("Adam needs step >= 1, lr > 0 and betas in [0, 1)");
@@ -1537,6 +1798,7 @@ static int check_readout(const deer_readout *r, int B, int T, int M) {
 // ---- sequential baseline -------------------------------------------------------------------
 static int check_sequential(const deer_model *m, const deer_forcing *f, int B, int T, SeqArgs *a) {
     if (!m || !f) { set_error("model/forcing pointer is NULL"); return DEER_ERR_INVALID_ARG; }
+    if (no_obs(f, "deer_sequential")) return DEER_ERR_INVALID_ARG;
     if (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN) {
         set_error("the sequential baseline covers the PLRNN kinds");
         return DEER_ERR_INVALID_ARG;

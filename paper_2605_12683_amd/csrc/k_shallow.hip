@@ -77,6 +77,8 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
             if (ok && i < M) {
                 if (s == 0) {
                     pz[r] = a.z0 ? a.z0[(size_t)b * M + i] : (i < N ? a.x[(size_t)b * (T + 1) * N + i] : 0.f);
+                } else if (a.zt) {
+                    pz[r] = a.zt[((size_t)b * T + s) * M + i];   // the forced input itself (N = 0)
                 } else {
                     pz[r] = z[((size_t)b * T + s - 1) * M + i];
                     if (i < N) px[r] = a.x[((size_t)b * (T + 1) + s) * N + i];
@@ -243,7 +245,10 @@ __global__ __launch_bounds__(256) void k_jacform_shplrnn(const ShArgs a, const u
     __syncthreads();
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, c = lane & 15;
     const int LW = (L + 31) / 32;
-    const long total = (long)a.B * T;
+    // rows (b, s) with t_lo <= s < t_hi, numbered b * len + (s - t_lo)
+    const int t_lo = a.t_hi > a.t_lo ? a.t_lo : 0;
+    const int len = a.t_hi > a.t_lo ? a.t_hi - a.t_lo : T;
+    const long total = (long)a.B * len;
     const long ngroups = (total + NT - 1) / NT;
     float dI[NI][4];
 #pragma unroll
@@ -256,10 +261,13 @@ __global__ __launch_bounds__(256) void k_jacform_shplrnn(const ShArgs a, const u
     for (long grp = (long)blockIdx.x * 4 + wv; grp < ngroups; grp += (long)gridDim.x * 4) {
         const long row0 = grp * NT;
         bool rok[NT];
+        long grow[NT];   // global row b * T + s of each of the NT rows
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             const long row = row0 + nt;
-            rok[nt] = row < total && (!active || active[row / T]);
+            const long b = row / len;
+            grow[nt] = b * T + t_lo + (row - b * len);
+            rok[nt] = row < total && (!active || active[b]);
         }
         v4f acc[NT][NI][NI];
 #pragma unroll
@@ -278,7 +286,7 @@ __global__ __launch_bounds__(256) void k_jacform_shplrnn(const ShArgs a, const u
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
                 if (!rok[nt]) continue;
-                const uint32_t w = masks[(size_t)(row0 + nt) * LW + word];
+                const uint32_t w = masks[(size_t)grow[nt] * LW + word];
 #pragma unroll
                 for (int Jt = 0; Jt < NI; ++Jt) {
                     const float b0 = select_bit(w, sh + 0, bv[Jt].x), b1 = select_bit(w, sh + 1, bv[Jt].y);
@@ -298,9 +306,9 @@ __global__ __launch_bounds__(256) void k_jacform_shplrnn(const ShArgs a, const u
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             if (!rok[nt]) continue;
-            float *Jp = Jout + (size_t)(row0 + nt) * M * M;
+            float *Jp = Jout + (size_t)grow[nt] * M * M;
             // damping of the linearisation of this sequence (1 = exact Newton)
-            const float gm = gamma ? gamma[(row0 + nt) / T] : 1.f;
+            const float gm = gamma ? gamma[grow[nt] / T] : 1.f;
 #pragma unroll
             for (int I = 0; I < NI; ++I)
 #pragma unroll
@@ -308,8 +316,10 @@ __global__ __launch_bounds__(256) void k_jacform_shplrnn(const ShArgs a, const u
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int row = 16 * I + 4 * g + r, col = 16 * Jt + c;
-                        if (row < M && col < M)
-                            Jp[row * M + col] = gm * (acc[nt][I][Jt][r] + (row == col ? dI[I][r] : 0.f));
+                        if (row < M && col < M) {
+                            const float d = a.Cd ? a.Cd[row * M + col] : (row == col ? dI[I][r] : 0.f);
+                            Jp[row * M + col] = gm * (acc[nt][I][Jt][r] + d);
+                        }
                     }
         }
     }
@@ -358,7 +368,7 @@ __global__ __launch_bounds__(SHG_THREADS) void k_grads_shplrnn(const ShArgs a, c
             float vz = 0.f, vl = 0.f;
             if (row < total && i < M) {
                 const int b = (int)(row / T), s = (int)(row % T);
-                vz = forced_state(a.x, a.z0, z, b, s, i, T, M, a.N, a.alpha);
+                vz = (a.zt && s > 0) ? a.zt[(size_t)row * M + i] : forced_state(a.x, a.z0, z, b, s, i, T, M, a.N, a.alpha);
                 vl = lam[(size_t)row * M + i];
             }
             zt[tt][i] = vz;
@@ -482,7 +492,7 @@ int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, con
     const int MP = padded_dim(a.M);
     const int LP = sh_LP(a.L);
     const size_t lds = sh_jacform_lds(a.M, a.L);
-    const long total = (long)a.B * a.T;
+    const long total = (long)a.B * (a.t_hi > a.t_lo ? a.t_hi - a.t_lo : a.T);
     KTimer kt("k_jacform_shplrnn", st);
 #define JF(MPV, NTV)                                                                                              \
     {                                                                                                             \

@@ -20,6 +20,15 @@ struct ShArgs {
     int N;
     const float *x, *z0;
     int B, T, M, L;
+    // general observation matrix (the forcing is formed outside these kernels; alpha = N = 0):
+    //   zt     [B,T,M]: zt[b, s] is the forced input z~_s of step s + 1 for s >= 1 (row 0 unused;
+    //          z~_0 = z0), read instead of forming it from z and x (residual, gradients)
+    //   Cd     [M,M]: dense term of the forced Jacobian, J~ = Cd + W1 diag(m) W2, replacing the
+    //          diagonal diag(A) P (Jacobian formation; W2 is then W2 P)
+    //   t_lo, t_hi: the Jacobian formation covers steps t_lo <= s < t_hi only (t_hi = 0: all)
+    const float *zt = nullptr;
+    const float *Cd = nullptr;
+    int t_lo = 0, t_hi = 0;
 };
 
 int padded_dim(int M);
@@ -203,6 +212,31 @@ size_t seq_part_floats(int M, int L, bool sh);
 int launch_seq_forward(const SeqArgs &a, float *z, float *act, hipStream_t st);
 int launch_seq_backward(const SeqArgs &a, const float *z, const float *act, const float *g, float seed_scale,
                         float *lam, float *part, const deer_grads *gr, hipStream_t st);
+
+// general observation matrix B [N, M] (k_obs.hip)
+struct ObsSetup {
+    const float *B;          // [N, M]
+    int N, M, L;             // L = hidden width (shallow) or M (vanilla, W2 = I)
+    float alpha;
+    const float *A, *W2;     // W2 null: the identity (vanilla PLRNN)
+    double *Bp64, *B64, *P164;                       // B^+ [M, N], B [N, M], P_1 [M, M]
+    float *Bp32, *Pa32, *P132, *Ca, *C1, *Id;        // B^+, P_alpha, P_1, diag(A) P_alpha, diag(A) P_1, I
+    float *Va, *V1;                                  // W2 P_alpha, W2 P_1 [L, M]
+    double *aug;                                     // [64][128] Gauss-Jordan scratch
+};
+int launch_obs_setup(const ObsSetup &s, hipStream_t st);
+// mode 0: forced inputs out[b, s] = P_s z_{s-1} + alpha_s B^+ x_s (s >= 1) of the current iterate;
+// mode 1: teacher states out[b, s] = B^+ x_{s+1}.  Both write z0e = B^+ x_0 when z0 is null.
+int launch_obs_forced(int mode, const float *z, const float *zalt, const int *zsel, const float *x, const float *z0,
+                      const float *Bp, const float *Pa, const float *P1, float alpha, int T_w, int B, int T, int M,
+                      int N, float *out, float *z0e, hipStream_t st);
+int launch_obs_seed(const float *z, const float *x, const float *Bm, float scale, int T_w, int B, int T, int M, int N,
+                    float *g, hipStream_t st);
+size_t obs_bgrad_ws_doubles(int M, int N);
+int launch_obs_bgrad(const float *JF, const float *lam, const float *z, const float *x, const float *Bm32,
+                     const double *Bp64, const double *Bm64, const double *P164, bool z0_given, float alpha, int T_w,
+                     bool with_mse, double mse_scale, int B, int T, int M, int N, double *ws, float *gB,
+                     hipStream_t st);
 
 // small utilities
 int launch_fill_teacher(int B, int T, int M, int N, const float *x, float *z, hipStream_t st);

@@ -156,3 +156,35 @@ def test_solve_with_tolerance_needs_the_threads_host_block(lib):
     assert out["q"] == _b.DEER_ERR_INVALID_ARG
     assert out["bad"] == _b.DEER_ERR_INVALID_ARG
     assert out["rel"] == _b.DEER_OK                 # nothing to free
+
+
+def test_observation_matrix_arguments(lib):
+    """A general observation matrix B: workspace queries for the solve, the adjoint and the
+    Jacobian entry point; n_forced (B's row count) in [1, 64], may exceed M; the entry points
+    that take the identity read-out only refuse it before any device work."""
+    m, _keep = _vanilla_model(8)
+    obs = (ctypes.c_float * 64)()
+    po = ctypes.cast(obs, ctypes.c_void_p)
+    f = _b.deer_forcing(0.1, 3, 0, po)
+    for op in (_b.DEER_OP_SOLVE, _b.DEER_OP_ADJOINT, _b.DEER_OP_JACOBIAN):
+        assert lib.deer_workspace_bytes_ex(ctypes.byref(m), ctypes.byref(f), 2, 64, op, 0) > 0
+    assert lib.deer_workspace_bytes_ex(ctypes.byref(m), ctypes.byref(f), 2, 64, _b.DEER_OP_SOLVE, 1) == 0  # quasi
+    tall = _b.deer_forcing(0.1, 12, 0, po)                 # N = 12 > M = 8
+    assert lib.deer_workspace_bytes_ex(ctypes.byref(m), ctypes.byref(tall), 2, 64, _b.DEER_OP_SOLVE, 0) > 0
+    for bad_n in (0, 65):
+        bad = _b.deer_forcing(0.1, bad_n, 0, po)
+        assert lib.deer_workspace_bytes_ex(ctypes.byref(m), ctypes.byref(bad), 2, 64, _b.DEER_OP_SOLVE, 0) == 0
+    dummy = (ctypes.c_float * 64)()
+    p = ctypes.cast(dummy, ctypes.c_void_p)
+    o = _b.deer_solve_opts(1e-5, 10, 2, 0, 0.0)
+    st = lib.deer_solve_quasi(ctypes.byref(m), ctypes.byref(f), ctypes.byref(o), 2, 8, p, None, p, None, None, None,
+                              p, 64, None)
+    assert st == _b.DEER_ERR_INVALID_ARG and b"observation" in lib.deer_last_error()
+    st = lib.plrnn_jacobian(ctypes.byref(m), ctypes.byref(f), 2, 8, p, None, p, p, None, None, None, None)
+    assert st == _b.DEER_ERR_INVALID_ARG and b"observation" in lib.deer_last_error()
+    gs = _b.deer_grads()
+    st = lib.deer_sequential(ctypes.byref(m), ctypes.byref(f), 2, 8, p, None, p, None, None, ctypes.byref(gs), p, 64,
+                             None)
+    assert st == _b.DEER_ERR_INVALID_ARG
+    dg = _b.deer_model(_b.DEER_DIAG_SSM, 4, 3, m.A, m.W, None, None, None)
+    assert lib.deer_workspace_bytes_ex(ctypes.byref(dg), ctypes.byref(f), 2, 64, _b.DEER_OP_SOLVE, 0) == 0

@@ -338,7 +338,7 @@ def fig1a_sweep(reps: int = 3):
     with variance 1/L), which is not a contraction for M >= 16 and makes DEER take many Newton
     updates; "contracting" rescales W1 so that max A + ||W1|| ||W2|| < 1 (A in [0.5, 0.65],
     ||W1|| ||W2|| = 0.3), the regime GTF is meant to produce.  DEER's iteration counts are those
-    of the model at hand.  The parallel solver covers M <= 64.  One JSON line per point."""
+    of the model at hand.  One JSON line per point."""
     import torch
     import workloads as W
     import paper_2605_12683_amd as D
@@ -379,17 +379,16 @@ def _fig1a_model(D, W, init, M, L, N, alpha, timed):
         seq_ms, _ = timed(lambda: D.deer_sequential(model, x, alpha, N, ws=ws_q, want_lam=False))
         rec = {"sweep": "fig1a", "model": "shplrnn", "init": init, "M": M, "L": L, "B": 1, "T": T, "alpha": alpha,
                "sequential_ms": round(seq_ms, 4), "deer_ms": None, "newton_updates": None, "speedup": None}
-        if M <= 64:
-            ws_s = D._workspace(D.deer_workspace_bytes(model, 1, T, 0))
-            ws_a = D._workspace(D.deer_workspace_bytes(model, 1, T, 1))
+        ws_s = D._workspace(D.deer_workspace_bytes(model, 1, T, 0))
+        ws_a = D._workspace(D.deer_workspace_bytes(model, 1, T, 1))
 
-            def step():
-                r = D.deer_solve(model, x, alpha, N, tol=1e-5, max_iter=500, ws=ws_s, check=False)
-                D.deer_adjoint(model, x, r["z"], alpha, N, ws=ws_a, want_lam=False)
-                return r
-            deer_ms, r = timed(step)
-            rec.update(deer_ms=round(deer_ms, 4), newton_updates=int(sum(r["iters"])),
-                       speedup=round(seq_ms / deer_ms, 3), status=int(r["status"]))
+        def step():
+            r = D.deer_solve(model, x, alpha, N, tol=1e-5, max_iter=500, ws=ws_s, check=False)
+            D.deer_adjoint(model, x, r["z"], alpha, N, ws=ws_a, want_lam=False)
+            return r
+        deer_ms, r = timed(step)
+        rec.update(deer_ms=round(deer_ms, 4), newton_updates=int(sum(r["iters"])),
+                   speedup=round(seq_ms / deer_ms, 3), status=int(r["status"]))
         print(json.dumps(rec), flush=True)
 
 

@@ -82,7 +82,9 @@ enum {
  * dimension (inputs u_t = x_{t-1}), other pointers unused. */
 typedef struct {
     int kind;
-    int M;              /* latent dimension: 1..64 for the PLRNN kinds, >= 1 for DIAG_SSM */
+    int M;              /* latent dimension: 1..64 for the vanilla PLRNN, 1..128 for the shallow
+                           one (M > 64: L <= 62, M L <= 7936; quasi-DEER and an observation
+                           matrix up to 64), >= 1 for DIAG_SSM */
     int L;              /* shallow: hidden width (1..1024); DIAG_SSM: input dimension       */
     const float *A;
     const float *W;
@@ -353,7 +355,7 @@ int plrnn_jacobian_ex(const deer_model *model, const deer_forcing *forcing, int 
  * `reverse` chooses the direction, `transpose` whether each step applies its matrix (0) or
  * its transpose (1); the Newton update of eq. GTF_DEER_update is (reverse, transpose) = (0, 0)
  * and the adjoint recursion of eq. backward_recursion is (1, 1).  With op(J) = J or J^T:
- *   DEER_SCAN_DENSE:    J [B,T,M,M] row-major per step, b [B,T,M], M <= 64.
+ *   DEER_SCAN_DENSE:    J [B,T,M,M] row-major per step, b [B,T,M], M <= 128.
  *        reverse == 0:  y_t = op(J_t) y_{t-1} + b_t, y_0 = 0        (J_1 is not read)
  *        reverse != 0:  y_T = b_T, y_{t-1} = op(J_t) y_t + b_{t-1}  (J_1 is not read)
  *   DEER_SCAN_DIAG_C64: J = lambda [M][2], b [B,T,M][2] complex; op(lambda) = lambda, or

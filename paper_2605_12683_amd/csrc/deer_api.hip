@@ -304,6 +304,15 @@ static int choose_chunk(int B, int T, int MP) {
     const long total = (long)B * T;
     // MP = 64 runs one chain per wave at two waves per SIMD: 8192 chains keep the tail of a
     // pass (fewer active sequences) spread over the machine
+    if (MP == 128) {
+        // one 4-wave workgroup per chain; fewer than 96 chunks per sequence (one carry level)
+        long C = (total + 1023) / 1024;
+        const long minC = (T + 94) / 95;
+        if (C < minC) C = minC;
+        if (C < 16) C = 16;
+        if (C > T) C = T;
+        return (int)C;
+    }
     const long target_chains = MP == 64 ? 8192L : 2048L * (64 / MP);
     long C = (total + target_chains - 1) / target_chains;
     if (C < 16) C = 16;
@@ -495,6 +504,14 @@ static int quasi_L(const deer_model *m) { return m->kind == DEER_SHPLRNN ? m->L 
 
 static int check_shallow_limits(const deer_model *m) {
     const size_t cap = 64 * 1024;
+    if (m->M > 64) {   // width-128 kernels: W1 and W2 in LDS
+        if (big_resjac_lds(m->M, m->L) > cap || big_jacform_lds(m->L) > cap || big_grads_lds(m->M, m->L) > cap) {
+            set_error("shallow PLRNN with M=%d, L=%d exceeds the 64 KiB LDS tiles of the width-128 kernels "
+                      "(M > 64 needs L <= 62 and M L <= 7936)", m->M, m->L);
+            return DEER_ERR_INVALID_ARG;
+        }
+        return DEER_OK;
+    }
     if (sh_resjac_lds(m->M, m->L) > cap || sh_jacform_lds(m->M, m->L) > cap) {
         set_error("shallow PLRNN with M=%d, L=%d exceeds the 64 KiB LDS tiles of this build (need M*L <= 8192 "
                   "for M <= 32)", m->M, m->L);
@@ -511,7 +528,11 @@ static int check_common(const deer_model *m, const deer_forcing *f, int B, int T
     if (!(f->alpha >= 0.0f && f->alpha <= 1.0f)) { set_error("alpha must lie in [0, 1]"); return DEER_ERR_INVALID_ARG; }
     if (m->M <= 0) { set_error("M must be positive"); return DEER_ERR_INVALID_ARG; }
     if (m->kind == DEER_PLRNN || m->kind == DEER_SHPLRNN) {
-        if (m->M > 64) { set_error("M=%d unsupported (dense scans support M <= 64)", m->M); return DEER_ERR_INVALID_ARG; }
+        const int mmax = m->kind == DEER_SHPLRNN && !f->obs ? 128 : 64;
+        if (m->M > mmax) {
+            set_error("M=%d unsupported (dense scans support M <= %d for this model and forcing)", m->M, mmax);
+            return DEER_ERR_INVALID_ARG;
+        }
         if (f->obs) {
             if (f->n_forced < 1 || f->n_forced > 64) {
                 set_error("with an observation matrix, n_forced (its row count) must lie in [1, 64]");
@@ -563,6 +584,10 @@ static int check_quasi(const deer_model *m, const deer_forcing *f, int B, int T)
     if ((rc = no_obs(f, "quasi-DEER"))) return rc;
     if (m->kind != DEER_PLRNN && m->kind != DEER_SHPLRNN) {
         set_error("quasi-DEER is built for the PLRNN kinds only");
+        return DEER_ERR_INVALID_ARG;
+    }
+    if (m->M > 64) {
+        set_error("quasi-DEER supports M <= 64");
         return DEER_ERR_INVALID_ARG;
     }
     if (m->kind == DEER_SHPLRNN) return check_shallow_limits(m);
@@ -1440,7 +1465,7 @@ size_t deer_scan_workspace_bytes(int layout, int reverse, int transpose, int B, 
     (void)transpose;
     if (B <= 0 || T <= 0 || M <= 0) return 0;
     if (layout == DEER_SCAN_DIAG_C64) return diag_scan_ws_bytes(B, T, M);
-    if (layout == DEER_SCAN_DENSE && M <= 64) {
+    if (layout == DEER_SCAN_DENSE && M <= 128) {
         size_t bytes = 0;
         carve_dense(nullptr, B, T, M, &bytes);
         return bytes;
@@ -1866,7 +1891,7 @@ int deer_scan(int layout, int reverse, int transpose, int B, int T, int M, const
         return launch_diag_scan(rev, B, T, M, J, b, nullptr, 0, nullptr, y, ws, st, tr ? 1 : 0);
     }
     if (layout == DEER_SCAN_DENSE) {
-        if (M > 64) { set_error("dense scans support M <= 64"); return DEER_ERR_INVALID_ARG; }
+        if (M > 128) { set_error("dense scans support M <= 128"); return DEER_ERR_INVALID_ARG; }
         size_t need = 0;
         carve_dense(nullptr, B, T, M, &need);
         int rc = check_ws(ws, ws_bytes, need);

@@ -1,0 +1,512 @@
+// Latent dimensions 65..128 (padded width 128) on the stored-Jacobian path of the shallow PLRNN:
+// the same operations as the M <= 64 kernels (k_dense.hip, k_shallow.hip, the carry walk), laid
+// out for a 128 x 128 chain matrix that one wave cannot hold.
+//
+//   k_chunk_product_big   one 4-wave workgroup per chain: wave w holds columns 32w..32w+31 of the
+//                         chunk product P <- E_t P in matrix-core accumulators (the previous step's
+//                         accumulators are the B operand, the step's Jacobian rows the A operand,
+//                         read as 16-byte vectors); the chunk-local solution u <- E_t u + rhs on
+//                         the vector units through LDS
+//   k_carry_big           one 128-thread block per sequence: carries across the chunks (fewer
+//                         than 96 per sequence at this width, so one level)
+//   k_fixup_big           one 128-thread block per chain: each chunk re-run from its carry
+//   k_resjac_big          residual, masks (the fixed-order float32 decision) and F, one row at a
+//                         time per block, W1 and W2 in LDS
+//   k_jacform_big         J~ = diag(A p) + W1 diag(m) (W2 P) on the matrix cores, 4 waves per
+//                         row, two column tiles each
+//   k_grads_big           per-block partial sums of the shallow gradients (layout of
+//                         k_grads_shplrnn), summed by k_reduce_rows
+// E_t is J_t, or J_t^T when flipped (the bare scan's other orientation), as in k_dense.hip.
+#include "common.h"
+#include "launch.h"
+
+namespace deer {
+
+constexpr int BG = 128;   // padded width
+
+// element (row, col) of E_t (J_t row-major per step, zero outside M x M)
+template <bool FLIP>
+__device__ __forceinline__ float eload(const float *__restrict__ Jp, int M, int row, int col) {
+    if (row >= M || col >= M) return 0.f;
+    return FLIP ? Jp[(size_t)col * M + row] : Jp[(size_t)row * M + col];
+}
+
+// REV: the product covers steps [s0 + 1, min(s1 + 1, T)) (the reverse chunk map is its
+// transpose) and the local solution runs u_k = E_{k+1}^T u_{k+1} + rhs_k from k = s1 - 1 down.
+template <bool REV, bool FLIP>
+__global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restrict__ J, const float *__restrict__ rhs,
+                                                           float rhs_sign, float *__restrict__ Pout,
+                                                           float *__restrict__ vout, const int *__restrict__ active,
+                                                           int B, int T, int M, int C, int ncs) {
+    __shared__ __align__(16) float ub[2][BG];
+    const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
+    const int id = blockIdx.x;   // chain
+    const int b = id / ncs, cc = id % ncs;
+    const bool ok = !active || active[b];
+    const int s0 = cc * C, s1 = min(s0 + C, T);
+    const int lo = REV ? s0 + 1 : s0, hi = REV ? min(s1 + 1, T) : s1;
+    const int plen = ok ? max(hi - lo, 0) : 0;
+    const int ulen = ok ? s1 - s0 : 0;
+    const int nsteps = max(plen, ulen);
+    // accumulators: acc[I][Jt][r] = P[16 I + 4 g + r][32 wv + 16 Jt + c]
+    v4f acc[8][2];
+#pragma unroll
+    for (int I = 0; I < 8; ++I)
+#pragma unroll
+        for (int Jt = 0; Jt < 2; ++Jt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[I][Jt][r] = (16 * I + 4 * g + r == 32 * wv + 16 * Jt + c) ? 1.f : 0.f;
+    // local solution: thread pair (row i = tid / 2, half hh) sums half of the row
+    const int ui = tid >> 1, hh = tid & 1;
+    if (tid < BG) ub[0][tid] = 0.f;
+    __syncthreads();
+    int cur = 0;
+    for (int t = 0; t < nsteps; ++t) {
+        if (t < plen) {
+            const float *Jp = J + ((size_t)b * T + lo + t) * M * M;
+            v4f old[8][2];
+#pragma unroll
+            for (int I = 0; I < 8; ++I)
+#pragma unroll
+                for (int Jt = 0; Jt < 2; ++Jt) {
+                    old[I][Jt] = acc[I][Jt];
+                    acc[I][Jt] = (v4f){0.f, 0.f, 0.f, 0.f};
+                }
+#pragma unroll
+            for (int I = 0; I < 8; ++I) {
+                const int row = 16 * I + c;
+                float a[8][4];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int k0 = 16 * j + 4 * g;
+                    if (!FLIP && row < M && k0 + 3 < M && (M & 3) == 0) {
+                        const float4 v = *reinterpret_cast<const float4 *>(Jp + (size_t)row * M + k0);
+                        a[j][0] = v.x; a[j][1] = v.y; a[j][2] = v.z; a[j][3] = v.w;
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) a[j][q] = eload<FLIP>(Jp, M, row, k0 + q);
+                    }
+                }
+#pragma unroll
+                for (int Jt = 0; Jt < 2; ++Jt) {
+                    v4f s = acc[I][Jt];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) s = mfma16x16x4(a[j][q], old[j][Jt][q], s);
+                    acc[I][Jt] = s;
+                }
+            }
+        }
+        if (t < ulen) {
+            // forward: u_s = E_s u_{s-1} + sign rhs_s, s = s0 + t;  reverse: k = s1 - 1 - t,
+            // u_k = E_{k+1}^T u_{k+1} + sign rhs_k (E_T does not exist: the first reverse step
+            // starts from zero)
+            const int k = REV ? s1 - 1 - t : s0 + t;
+            const int kj = REV ? k + 1 : k;
+            float part = 0.f;
+            if (ui < M && (!REV || kj < T)) {
+                const float *Jp = J + ((size_t)b * T + kj) * M * M;
+                for (int q = hh; q < M; q += 2) {
+                    // forward: row ui of E; reverse: column ui of E (row ui of E^T)
+                    const float e = REV ? eload<FLIP>(Jp, M, q, ui) : eload<FLIP>(Jp, M, ui, q);
+                    part = fmaf(e, ub[cur][q], part);
+                }
+            }
+            part += __shfl_xor(part, 1, 64);
+            if (hh == 0 && ui < BG)
+                ub[cur ^ 1][ui] = ui < M ? fmaf(rhs_sign, rhs[((size_t)b * T + k) * M + ui], part) : 0.f;
+            __syncthreads();
+            cur ^= 1;
+        }
+    }
+    if (!ok) return;
+    float *P = Pout + (size_t)id * BG * BG;
+#pragma unroll
+    for (int I = 0; I < 8; ++I)
+#pragma unroll
+        for (int Jt = 0; Jt < 2; ++Jt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) P[(16 * I + 4 * g + r) * BG + 32 * wv + 16 * Jt + c] = acc[I][Jt][r];
+    if (tid < BG) vout[(size_t)id * BG + tid] = ub[cur][tid];
+}
+
+// carries across the chunks of each sequence, in processing order (REV: from the last chunk):
+// carry_in[c] = the state entering chunk c;  next = A_c carry + v_c with A_c = P_c (P_c^T in REV)
+template <bool REV>
+__global__ __launch_bounds__(BG) void k_carry_big(const float *__restrict__ P, const float *__restrict__ v,
+                                                  float *__restrict__ carry_in, const int *__restrict__ active,
+                                                  int ncs) {
+    __shared__ float cs[BG];
+    const int b = blockIdx.x, i = threadIdx.x;
+    if (active && !active[b]) return;
+    float cur = 0.f;
+    for (int step = 0; step < ncs; ++step) {
+        const int cc = REV ? ncs - 1 - step : step;
+        const size_t id = (size_t)b * ncs + cc;
+        carry_in[id * BG + i] = cur;
+        cs[i] = cur;
+        __syncthreads();
+        const float *Pc = P + id * BG * BG;
+        float a = v[id * BG + i];
+        for (int k = 0; k < BG; ++k) a = fmaf(REV ? Pc[(size_t)k * BG + i] : Pc[(size_t)i * BG + k], cs[k], a);
+        __syncthreads();
+        cur = a;
+    }
+}
+
+// MODE 0: Newton fix-up (next iterate = current + Delta, per-chain max |Delta| and max |z|);
+// MODE 1: forward bare scan; MODE 2: reverse (y_k = E_{k+1}^T y_{k+1} + b_k)
+template <int MODE, bool FLIP>
+__global__ __launch_bounds__(BG) void k_fixup_big(const float *__restrict__ J, const float *__restrict__ rhs,
+                                                  float rhs_sign, const float *__restrict__ carry_in, float *zbuf,
+                                                  float *outbuf, const int *__restrict__ zsel,
+                                                  uint32_t *__restrict__ chain_bits, const int *__restrict__ active,
+                                                  int B, int T, int M, int C, int ncs) {
+    __shared__ float ys[2][BG];
+    __shared__ uint32_t red[2][BG / 64];
+    const int id = blockIdx.x, i = threadIdx.x;
+    const int b = id / ncs, cc = id % ncs;
+    const bool ok = !active || active[b];
+    const int s0 = cc * C, s1 = ok ? min(s0 + C, T) : s0;
+    const float *zin = MODE == 0 ? cur_iter(zbuf, outbuf, zsel, b) : nullptr;
+    float *out = MODE == 0 ? next_iter(zbuf, outbuf, zsel, b) : outbuf;
+    ys[0][i] = (ok && i < M) ? carry_in[(size_t)id * BG + i] : 0.f;
+    __syncthreads();
+    uint32_t emax = 0u, zmax = 0u;
+    int cur = 0;
+    for (int t = 0; t < s1 - s0; ++t) {
+        const int k = MODE == 2 ? s1 - 1 - t : s0 + t;
+        const int kj = MODE == 2 ? k + 1 : k;
+        float acc = 0.f;
+        if (i < M && kj < T) {
+            const float *Jp = J + ((size_t)b * T + kj) * M * M;
+            for (int q = 0; q < M; ++q) {
+                const float e = MODE == 2 ? eload<FLIP>(Jp, M, q, i) : eload<FLIP>(Jp, M, i, q);
+                acc = fmaf(e, ys[cur][q], acc);
+            }
+        }
+        float y = 0.f;
+        if (i < M) {
+            const size_t e = ((size_t)b * T + k) * M + i;
+            y = fmaf(rhs_sign, rhs[e], acc);
+            if (MODE == 0) {
+                const float zo = zin[e];
+                out[e] = zo + y;
+                const uint32_t ab = abs_bits(y), zb = abs_bits(zo);
+                emax = emax > ab ? emax : ab;
+                zmax = zmax > zb ? zmax : zb;
+            } else {
+                out[e] = y;
+            }
+        }
+        ys[cur ^ 1][i] = y;
+        __syncthreads();
+        cur ^= 1;
+    }
+    if (MODE == 0) {
+        emax = wave_max_u32(emax);
+        zmax = wave_max_u32(zmax);
+        if ((i & 63) == 0) {
+            red[0][i >> 6] = emax;
+            red[1][i >> 6] = zmax;
+        }
+        __syncthreads();
+        if (i == 0 && ok) {
+            const uint32_t e = red[0][0] > red[0][1] ? red[0][0] : red[0][1];
+            const uint32_t z = red[1][0] > red[1][1] ? red[1][0] : red[1][1];
+            chain_bits[id] = e;
+            chain_bits[(size_t)B * ncs + id] = z;
+        }
+    }
+}
+
+// ---- shallow PLRNN at M <= 128 -------------------------------------------------------------
+
+// forced input of step s for latent i, the float32 decision of the other kernels
+__device__ __forceinline__ float big_forced(const ShArgs &a, const float *z, int b, int s, int i) {
+    if (s == 0) return a.z0 ? a.z0[(size_t)b * a.M + i] : (i < a.N ? a.x[(size_t)b * (a.T + 1) * a.N + i] : 0.f);
+    if (a.zt) return a.zt[((size_t)b * a.T + s) * a.M + i];
+    const float zp = z[((size_t)b * a.T + s - 1) * a.M + i];
+    if (i >= a.N) return zp;
+    const float p = __fsub_rn(1.0f, a.alpha);
+    return __fadd_rn(__fmul_rn(p, zp), __fmul_rn(a.alpha, a.x[((size_t)b * (a.T + 1) + s) * a.N + i]));
+}
+
+// LDS: W1 [M][L] | W2 [L][M] | z~ [BG] | relu(u) [L]
+__global__ __launch_bounds__(256) void k_resjac_big(const ShArgs a, const float *zbuf, const float *zalt,
+                                                    const int *__restrict__ zsel, float *__restrict__ F_out,
+                                                    float *__restrict__ r_out, uint32_t *__restrict__ masks,
+                                                    const int *__restrict__ active) {
+    extern __shared__ __align__(16) float smem[];
+    const int M = a.M, L = a.L, T = a.T, tid = threadIdx.x;
+    float *w1 = smem, *w2 = w1 + (size_t)M * L, *zt = w2 + (size_t)L * M, *ru = zt + BG;
+    for (int e = tid; e < M * L; e += 256) {
+        w1[e] = a.W1[e];
+        w2[e] = a.W2[e];
+    }
+    const int LW = (L + 31) / 32;
+    const long rows = (long)a.B * T;
+    __syncthreads();
+    for (long row = blockIdx.x; row < rows; row += gridDim.x) {
+        const int b = (int)(row / T), s = (int)(row % T);
+        const bool on = !active || active[b];   // block-uniform
+        if (!on) continue;
+        const float *z = cur_iter(zbuf, zalt, zsel, b);
+        if (tid < M) zt[tid] = big_forced(a, z, b, s, tid);
+        __syncthreads();
+        // hidden pre-activations left to right from h2, a rounding after every multiply and add
+        for (int l = tid; l < L; l += 256) {
+            float u = a.h2 ? a.h2[l] : 0.f;
+            for (int j = 0; j < M; ++j) u = __fadd_rn(u, __fmul_rn(w2[(size_t)l * M + j], zt[j]));
+            ru[l] = u > 0.f ? u : 0.f;
+        }
+        __syncthreads();
+        if (masks) {
+            for (int w = tid; w < LW; w += 256) {
+                uint32_t bits = 0u;
+                for (int k = 0; k < 32; ++k) {
+                    const int l = 32 * w + k;
+                    if (l < L && ru[l] > 0.f) bits |= 1u << k;
+                }
+                masks[(size_t)row * LW + w] = bits;
+            }
+        }
+        if (tid < M) {
+            float f = 0.f;
+            for (int l = 0; l < L; ++l) f = fmaf(w1[(size_t)tid * L + l], ru[l], f);
+            f = fmaf(a.A[tid], zt[tid], f) + (a.h1 ? a.h1[tid] : 0.f);
+            const size_t e = (size_t)row * M + tid;
+            if (F_out) F_out[e] = f;
+            if (r_out) r_out[e] = z[e] - f;
+        }
+        __syncthreads();
+    }
+}
+
+// J~_s = Cd (or diag(A p)) + W1 diag(m_s) V with V = W2 diag(p) (or the given W2 P): one row per
+// block, wave wv computes the column tiles 2 wv, 2 wv + 1 of all 8 row tiles.  LDS: W1 [BG][LP],
+// V^T [BG][LP], zero padded (LP = L rounded up to 16).
+__global__ __launch_bounds__(256) void k_jacform_big(const ShArgs a, const uint32_t *__restrict__ masks,
+                                                     float *__restrict__ Jout, const int *__restrict__ active,
+                                                     const float *__restrict__ gamma, int LP) {
+    extern __shared__ __align__(16) float smem[];
+    const int M = a.M, L = a.L, T = a.T, N = a.N;
+    float *w1s = smem, *vts = smem + BG * LP;
+    const int tid = threadIdx.x;
+    const float p1 = __fsub_rn(1.0f, a.alpha);
+    for (int e = tid; e < BG * LP; e += 256) {
+        const int i = e / LP, l = e % LP;
+        const bool in = i < M && l < L;
+        w1s[e] = in ? a.W1[(size_t)i * L + l] : 0.f;
+        vts[e] = in ? a.W2[(size_t)l * M + i] * (i < N ? p1 : 1.f) : 0.f;
+    }
+    __syncthreads();
+    const int wv = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
+    const int LW = (L + 31) / 32;
+    const int t_lo = a.t_hi > a.t_lo ? a.t_lo : 0;
+    const int len = a.t_hi > a.t_lo ? a.t_hi - a.t_lo : T;
+    const long rows = (long)a.B * len;
+    for (long r0 = blockIdx.x; r0 < rows; r0 += gridDim.x) {
+        const long bb = r0 / len;
+        const long grow = bb * T + t_lo + (r0 - bb * len);
+        if (active && !active[bb]) continue;
+        v4f acc[8][2];
+#pragma unroll
+        for (int I = 0; I < 8; ++I)
+#pragma unroll
+            for (int Jt = 0; Jt < 2; ++Jt) acc[I][Jt] = (v4f){0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < LP / 16; ++j) {
+            const int word = (16 * j) >> 5, sh = 16 * (j & 1) + 4 * g;
+            const uint32_t w = masks[(size_t)grow * LW + word];
+            float4 bv[2];
+#pragma unroll
+            for (int Jt = 0; Jt < 2; ++Jt) {
+                const float4 t4 = *reinterpret_cast<const float4 *>(vts + (32 * wv + 16 * Jt + c) * LP + 16 * j + 4 * g);
+                bv[Jt] = make_float4(select_bit(w, sh, t4.x), select_bit(w, sh + 1, t4.y), select_bit(w, sh + 2, t4.z),
+                                     select_bit(w, sh + 3, t4.w));
+            }
+#pragma unroll
+            for (int I = 0; I < 8; ++I) {
+                const float4 av = *reinterpret_cast<const float4 *>(w1s + (16 * I + c) * LP + 16 * j + 4 * g);
+#pragma unroll
+                for (int Jt = 0; Jt < 2; ++Jt) {
+                    v4f t = acc[I][Jt];
+                    t = mfma16x16x4(av.x, bv[Jt].x, t);
+                    t = mfma16x16x4(av.y, bv[Jt].y, t);
+                    t = mfma16x16x4(av.z, bv[Jt].z, t);
+                    t = mfma16x16x4(av.w, bv[Jt].w, t);
+                    acc[I][Jt] = t;
+                }
+            }
+        }
+        float *Jp = Jout + (size_t)grow * M * M;
+        const float gm = gamma ? gamma[bb] : 1.f;
+#pragma unroll
+        for (int I = 0; I < 8; ++I)
+#pragma unroll
+            for (int Jt = 0; Jt < 2; ++Jt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = 16 * I + 4 * g + r, col = 32 * wv + 16 * Jt + c;
+                    if (row < M && col < M) {
+                        const float d = a.Cd ? a.Cd[row * M + col]
+                                             : (row == col ? a.A[row] * (row < N ? p1 : 1.f) : 0.f);
+                        Jp[row * M + col] = gm * (acc[I][Jt][r] + d);
+                    }
+                }
+    }
+}
+
+// Per-block partial sums over rows (layout of k_grads_shplrnn):
+//   [M*L dW1 (row-major) | L*M dW2 | L dh2 | M dA | M dh1]
+// dW1 += lam relu(u)^T, dW2 += delta z~^T with delta = (W1^T lam) * m, dh2 += delta, dA += lam * z~,
+// dh1 += lam.  Each thread owns up to GB_PER entries of dW1 and of dW2 in registers.
+constexpr int GB_PER = 32;
+
+__global__ __launch_bounds__(256) void k_grads_big(const ShArgs a, const float *__restrict__ z,
+                                                   const float *__restrict__ lam, const uint32_t *__restrict__ masks,
+                                                   float *__restrict__ part) {
+    extern __shared__ __align__(16) float smem[];
+    const int M = a.M, L = a.L, T = a.T, tid = threadIdx.x;
+    float *w1 = smem, *w2 = w1 + (size_t)M * L, *zt = w2 + (size_t)L * M, *lm = zt + BG, *ru = lm + BG,
+          *dl = ru + L;
+    for (int e = tid; e < M * L; e += 256) {
+        w1[e] = a.W1[e];
+        w2[e] = a.W2[e];
+    }
+    const int LW = (L + 31) / 32;
+    float g1[GB_PER], g2[GB_PER];
+#pragma unroll
+    for (int q = 0; q < GB_PER; ++q) g1[q] = g2[q] = 0.f;
+    float dh2 = 0.f, dA = 0.f, dh1 = 0.f;
+    const long rows = (long)a.B * T;
+    const long per = (rows + gridDim.x - 1) / gridDim.x;
+    const long r0 = (long)blockIdx.x * per, r1 = r0 + per < rows ? r0 + per : rows;
+    __syncthreads();
+    for (long row = r0; row < r1; ++row) {
+        const int b = (int)(row / T), s = (int)(row % T);
+        if (tid < M) {
+            zt[tid] = big_forced(a, z, b, s, tid);
+            lm[tid] = lam[(size_t)row * M + tid];
+        }
+        __syncthreads();
+        for (int l = tid; l < L; l += 256) {
+            const bool m = (masks[(size_t)row * LW + (l >> 5)] >> (l & 31)) & 1u;
+            float u = a.h2 ? a.h2[l] : 0.f, d = 0.f;
+            for (int k = 0; k < M; ++k) {
+                u = fmaf(w2[(size_t)l * M + k], zt[k], u);
+                d = fmaf(w1[(size_t)k * L + l], lm[k], d);
+            }
+            ru[l] = m ? u : 0.f;
+            dl[l] = m ? d : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < GB_PER; ++q) {
+            const int e = tid + 256 * q;
+            if (e < M * L) {
+                g1[q] = fmaf(lm[e / L], ru[e % L], g1[q]);      // dW1[i][l]
+                g2[q] = fmaf(dl[e / M], zt[e % M], g2[q]);      // dW2[l][j]
+            }
+        }
+        if (tid < L) dh2 += dl[tid];
+        if (tid < M) {
+            dA = fmaf(lm[tid], zt[tid], dA);
+            dh1 += lm[tid];
+        }
+        __syncthreads();
+    }
+    const size_t stride = (size_t)2 * M * L + L + 2 * M;
+    float *pp = part + (size_t)blockIdx.x * stride;
+#pragma unroll
+    for (int q = 0; q < GB_PER; ++q) {
+        const int e = tid + 256 * q;
+        if (e < M * L) {
+            pp[e] = g1[q];
+            pp[(size_t)M * L + e] = g2[q];
+        }
+    }
+    if (tid < L) pp[(size_t)2 * M * L + tid] = dh2;
+    if (tid < M) {
+        pp[(size_t)2 * M * L + L + tid] = dA;
+        pp[(size_t)2 * M * L + L + M + tid] = dh1;
+    }
+}
+
+// ---- host launchers (called by the dispatchers of the M <= 64 kernels when the padded width is
+// 128) ------------------------------------------------------------------------------------------
+
+int launch_chunk_product_big(bool rev, bool flip, int B, int T, int M, const float *J, const float *rhs,
+                             float rhs_sign, float *P, float *v, const int *active, int C, int ncs, hipStream_t st) {
+    const int grid = B * ncs;
+    KTimer kt("k_chunk_product_dense", st);
+#define CPB(R, F) \
+    hipLaunchKernelGGL((k_chunk_product_big<R, F>), dim3(grid), dim3(256), 0, st, J, rhs, rhs_sign, P, v, active, B, T, M, C, ncs)
+    if (!rev) { if (flip) CPB(false, true); else CPB(false, false); }
+    else { if (flip) CPB(true, true); else CPB(true, false); }
+#undef CPB
+    DEER_LAUNCH_CHECK("k_chunk_product_big");
+    return DEER_OK;
+}
+
+int launch_carry_big(bool rev, const float *P, const float *v, float *carry_in, const int *active, int B, int ncs,
+                     hipStream_t st) {
+    KTimer kt("k_carry", st);
+    if (rev) hipLaunchKernelGGL(k_carry_big<true>, dim3(B), dim3(BG), 0, st, P, v, carry_in, active, ncs);
+    else hipLaunchKernelGGL(k_carry_big<false>, dim3(B), dim3(BG), 0, st, P, v, carry_in, active, ncs);
+    DEER_LAUNCH_CHECK("k_carry_big");
+    return DEER_OK;
+}
+
+int launch_fixup_big(int mode, bool flip, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
+                     const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
+                     const int *active, int C, int ncs, hipStream_t st) {
+    const int grid = B * ncs;
+    KTimer kt(mode == 2 ? "k_fixup_dense_rev" : "k_fixup_dense_fwd", st);
+#define FXB(MO, F)                                                                                                  \
+    hipLaunchKernelGGL((k_fixup_big<MO, F>), dim3(grid), dim3(BG), 0, st, J, rhs, rhs_sign, carry_in, z, out, zsel, \
+                       chain_bits, active, B, T, M, C, ncs)
+    if (mode == 0) FXB(0, false);
+    else if (mode == 1) { if (flip) FXB(1, true); else FXB(1, false); }
+    else { if (flip) FXB(2, true); else FXB(2, false); }
+#undef FXB
+    DEER_LAUNCH_CHECK("k_fixup_big");
+    return DEER_OK;
+}
+
+size_t big_resjac_lds(int M, int L) { return ((size_t)2 * M * L + BG + L) * sizeof(float); }
+size_t big_jacform_lds(int L) { return (size_t)2 * BG * ((L + 15) / 16 * 16) * sizeof(float); }
+size_t big_grads_lds(int M, int L) { return ((size_t)2 * M * L + 2 * BG + 2 * L) * sizeof(float); }
+
+int launch_resjac_big(const ShArgs &a, const float *z, const float *zalt, const int *zsel, float *F, float *r,
+                      uint32_t *masks, const int *active, hipStream_t st) {
+    const long rows = (long)a.B * a.T;
+    const int grid = (int)(rows < 8192 ? rows : 8192);
+    KTimer kt("k_resjac_shplrnn", st);
+    hipLaunchKernelGGL(k_resjac_big, dim3(grid), dim3(256), big_resjac_lds(a.M, a.L), st, a, z, zalt, zsel, F, r,
+                       masks, active);
+    DEER_LAUNCH_CHECK("k_resjac_big");
+    return DEER_OK;
+}
+
+int launch_jacform_big(const ShArgs &a, const uint32_t *masks, float *J, const int *active, const float *gamma,
+                       hipStream_t st) {
+    const long rows = (long)a.B * (a.t_hi > a.t_lo ? a.t_hi - a.t_lo : a.T);
+    const int grid = (int)(rows < 8192 ? rows : 8192);
+    const int LP = (a.L + 15) / 16 * 16;
+    KTimer kt("k_jacform_shplrnn", st);
+    hipLaunchKernelGGL(k_jacform_big, dim3(grid), dim3(256), big_jacform_lds(a.L), st, a, masks, J, active, gamma, LP);
+    DEER_LAUNCH_CHECK("k_jacform_big");
+    return DEER_OK;
+}
+
+int launch_grads_big(const ShArgs &a, const float *z, const float *lam, const uint32_t *masks, float *part, int nb,
+                     hipStream_t st) {
+    KTimer kt("k_grads_shplrnn", st);
+    hipLaunchKernelGGL(k_grads_big, dim3(nb), dim3(256), big_grads_lds(a.M, a.L), st, a, z, lam, masks, part);
+    DEER_LAUNCH_CHECK("k_grads_big");
+    return DEER_OK;
+}
+
+}  // namespace deer

@@ -408,6 +408,7 @@ __global__ __launch_bounds__(64) void k_fixup_dense(const float *__restrict__ J,
 int launch_chunk_product_dense(bool rev, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
                                float *P, float *v, const int *active, int C, int ncs, hipStream_t st, bool flip) {
     const int MP = padded_dim(M);
+    if (MP == 128) return launch_chunk_product_big(rev, flip, B, T, M, J, rhs, rhs_sign, P, v, active, C, ncs, st);
     const int nch = B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt("k_chunk_product_dense", st);
@@ -436,6 +437,9 @@ int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const floa
                        const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
                        const int *active, int C, int ncs, hipStream_t st, bool flip) {
     const int MP = padded_dim(M);
+    if (MP == 128)
+        return launch_fixup_big(mode, flip, B, T, M, J, rhs, rhs_sign, carry_in, z, out, zsel, chain_bits, active, C,
+                                ncs, st);
     const int nch = B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt(mode == 2 ? "k_fixup_dense_rev" : "k_fixup_dense_fwd", st);

@@ -2966,7 +2966,7 @@ static int invalid_arg(const char *what) {
     return DEER_ERR_INVALID_ARG;
 }
 
-static int padded(int M) { return M <= 16 ? 16 : (M <= 32 ? 32 : 64); }
+static int padded(int M) { return M <= 16 ? 16 : (M <= 32 ? 32 : (M <= 64 ? 64 : 128)); }
 
 int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, float *J, uint32_t *masks,
                         const int *active, hipStream_t st) {
@@ -3078,6 +3078,10 @@ size_t carry_ws_floats(int MP, int B, int ncs) {
 
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
                  uint32_t *norm_bits, int B, int ncs, float *gws, hipStream_t st) {
+    if (MP == 128) {
+        if (norm_bits || carry_group_size(MP, ncs)) return invalid_arg("width-128 carries take one level, no norms");
+        return launch_carry_big(rev, P, v, carry_in, active, B, ncs, st);
+    }
     KTimer kt("k_carry", st);
     const int G = gws ? carry_group_size(MP, ncs) : 0;
 #define CA(MPV, R, PP, VV, CI, NB, NC, GG, ST, GRID) \

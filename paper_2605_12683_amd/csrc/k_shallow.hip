@@ -474,6 +474,7 @@ size_t sh_jacform_lds(int M, int L) { return (size_t)2 * padded_dim(M) * sh_LP(L
 
 int launch_resjac_shplrnn(const ShArgs &a, const float *z, const float *zalt, const int *zsel, float *F, float *r,
                           uint32_t *masks, const int *active, hipStream_t st) {
+    if (padded_dim(a.M) == 128) return launch_resjac_big(a, z, zalt, zsel, F, r, masks, active, st);
     const long ntiles = ((long)a.B * a.T + SH_TT - 1) / SH_TT;
     const int grid = (int)(ntiles < 4096 ? ntiles : 4096);
     const size_t lds = sh_resjac_lds(a.M, a.L);
@@ -489,6 +490,7 @@ int launch_resjac_shplrnn(const ShArgs &a, const float *z, const float *zalt, co
 
 int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, const int *active, const float *gamma,
                            hipStream_t st) {
+    if (padded_dim(a.M) == 128) return launch_jacform_big(a, masks, J, active, gamma, st);
     const int MP = padded_dim(a.M);
     const int LP = sh_LP(a.L);
     const size_t lds = sh_jacform_lds(a.M, a.L);
@@ -519,7 +521,10 @@ int launch_grads_shplrnn(const ShArgs &a, const float *z, const float *lam, cons
     sh_grads_part_floats(a.M, a.L, &nb);
     const int MP = padded_dim(a.M);
     const dim3 grid(nb, (a.L + SHG_THREADS - 1) / SHG_THREADS);
-    {
+    if (MP == 128) {
+        int rc = launch_grads_big(a, z, lam, masks, part, nb, st);
+        if (rc) return rc;
+    } else {
         KTimer kt("k_grads_shplrnn", st);
         if (MP == 16) hipLaunchKernelGGL(k_grads_shplrnn<16>, grid, dim3(SHG_THREADS), 0, st, a, z, lam, masks, part);
         else if (MP == 32) hipLaunchKernelGGL(k_grads_shplrnn<32>, grid, dim3(SHG_THREADS), 0, st, a, z, lam, masks, part);

@@ -164,6 +164,25 @@ int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const floa
                        const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
                        const int *active, int C, int ncs, hipStream_t st, bool flip = false);
 
+// latent dimensions 65..128 (padded width 128; k_big.hip), dispatched to by the launchers above
+// and below; the carry has one level (fewer than 96 chunks per sequence at this width)
+int launch_chunk_product_big(bool rev, bool flip, int B, int T, int M, const float *J, const float *rhs,
+                             float rhs_sign, float *P, float *v, const int *active, int C, int ncs, hipStream_t st);
+int launch_carry_big(bool rev, const float *P, const float *v, float *carry_in, const int *active, int B, int ncs,
+                     hipStream_t st);
+int launch_fixup_big(int mode, bool flip, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
+                     const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
+                     const int *active, int C, int ncs, hipStream_t st);
+size_t big_resjac_lds(int M, int L);
+size_t big_jacform_lds(int L);
+size_t big_grads_lds(int M, int L);
+int launch_resjac_big(const ShArgs &a, const float *z, const float *zalt, const int *zsel, float *F, float *r,
+                      uint32_t *masks, const int *active, hipStream_t st);
+int launch_jacform_big(const ShArgs &a, const uint32_t *masks, float *J, const int *active, const float *gamma,
+                       hipStream_t st);
+int launch_grads_big(const ShArgs &a, const float *z, const float *lam, const uint32_t *masks, float *part, int nb,
+                     hipStream_t st);
+
 // shallow PLRNN
 size_t sh_resjac_lds(int M, int L);
 size_t sh_jacform_lds(int M, int L);

@@ -1,0 +1,119 @@
+"""Latent dimensions 65..128 (the width-128 kernels) on the GPU: the shallow PLRNN of the Fig. 1A
+grid (L = 50, M up to 128) solved and differentiated by the parallel solver, against the float64
+oracle and the sequential baseline, and the bare dense scan at these widths."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from gpu_util import masks_to_bool, oracle_model, rel_inf, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2605_12683_amd as D  # noqa: E402
+from paper_2605_12683_amd import _binding as Bnd  # noqa: E402
+
+TOL = 1e-4
+
+
+@pytest.fixture(autouse=True)
+def _no_chunk_override():
+    os.environ.pop("DEER_CHUNK", None)
+    yield
+    os.environ.pop("DEER_CHUNK", None)
+
+
+def _case(M, L, N, B, T, alpha, seed):
+    return W.random_shplrnn_case(M, L, N, B, T, alpha, seed, w_norm=0.3, a_range=(0.3, 0.6))
+
+
+@pytest.mark.parametrize("M,L,N,T", [(65, 7, 3, 40), (100, 50, 3, 70), (128, 50, 3, 60), (128, 62, 128, 33)])
+def test_big_jacobian_masks_bitexact(M, L, N, T):
+    """Residual, F and the masks (the fixed-order float32 decision) bit for bit in the masks, and
+    the dense forced Jacobians J~ = diag(A p) + W1 diag(m) W2 diag(p), at a given trajectory."""
+    c = _case(M, L, N, 2, T, 0.15, 1500 + M + L)
+    m = oracle_model(c)
+    z = np.random.default_rng(3).standard_normal((2, T, M)).astype(np.float32)
+    say("plrnn_jacobian big", M, L, N, T)
+    out = D.plrnn_jacobian(m, c.x, z, c.alpha, N, want=("F", "r", "masks"), dense_J=True)
+    idx = [(b, t) for b in range(2) for t in range(T)]
+    ref = O.jacobian_at(m, c.x, z, c.alpha, N, mask_precision="float32", dense_index=idx)
+    assert np.array_equal(masks_to_bool(out["masks"].cpu().numpy(), L), ref["mask"])
+    assert rel_inf(out["F"].cpu().numpy(), ref["F"]) < 1e-5
+    assert rel_inf(out["r"].cpu().numpy(), ref["r"]) < 1e-5
+    assert rel_inf(out["J"].cpu().numpy().reshape(-1, M, M), ref["J"]) < 1e-5
+
+
+@pytest.mark.parametrize("B,T,M,chunk", [(2, 300, 65, 0), (1, 1000, 128, 0), (2, 513, 128, 37), (1, 1, 100, 0)])
+@pytest.mark.parametrize("rev,tr", [(False, False), (True, True), (False, True), (True, False)])
+def test_big_dense_scan(B, T, M, chunk, rev, tr):
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    rng = np.random.default_rng(B * T + M)
+    J = (rng.standard_normal((B, T, M, M)) * (0.45 / np.sqrt(M))).astype(np.float32)
+    b = rng.standard_normal((B, T, M)).astype(np.float32)
+    say("deer_scan big", B, T, M, chunk, rev, tr)
+    y = D.deer_scan(Bnd.DEER_SCAN_DENSE, torch.tensor(J), torch.tensor(b), reverse=rev, transpose=tr).cpu().numpy()
+    Jd = J.astype(np.float64)
+    Jop = Jd if rev == tr else np.ascontiguousarray(np.swapaxes(Jd, -1, -2))
+    if rev:
+        ref = O.reverse_affine_recurrence(lambda k, w: np.einsum("bi,bij->bj", w, Jop[:, k]), b.astype(np.float64))
+    else:
+        ref = O.affine_recurrence(lambda k, v: np.einsum("bij,bj->bi", Jop[:, k], v), b.astype(np.float64))
+    assert rel_inf(y, ref) < TOL
+
+
+@pytest.mark.parametrize("M,L,N,B,T,alpha,chunk", [(128, 50, 3, 1, 2000, 0.15, 0), (128, 50, 3, 2, 700, 0.15, 41),
+                                                   (96, 30, 96, 2, 500, 0.1, 0), (128, 50, 3, 1, 1, 0.15, 0),
+                                                   (72, 20, 5, 3, 300, 0.3, 16)])
+def test_big_shallow_solve_and_adjoint(M, L, N, B, T, alpha, chunk):
+    """The parallel solve reaches the sequential rollout; the adjoint and every gradient equal the
+    oracle's recursion at the rollout (the ReLU decisions taken in float32 on both sides)."""
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    c = _case(M, L, N, B, T, alpha, 1600 + M + T)
+    m = oracle_model(c)
+    say("deer_solve big shallow", M, L, N, B, T, alpha, chunk)
+    res = D.deer_solve(m, c.x, alpha, N, tol=1e-5, max_iter=200)
+    assert res["status"] == 0, res
+    ref = O.rollout(m, c.x, alpha, N)
+    assert rel_inf(res["z"].cpu().numpy(), ref) < TOL
+    z32 = ref.astype(np.float32)
+    say("deer_adjoint big shallow", M, L, N, B, T, alpha, chunk)
+    out = D.deer_adjoint(m, c.x, z32, alpha, N)
+    lam = O.adjoint(m, c.x, z32, alpha, N, mask_precision="float32")
+    gr = O.param_grads(m, c.x, z32, alpha, N, lam, mask_precision="float32")
+    assert rel_inf(out["lam"].cpu().numpy(), lam) < TOL
+    for k in ("A", "W1", "W2", "h1", "h2"):
+        assert rel_inf(out["grads"][k].cpu().numpy(), gr[k]) < TOL, k
+
+
+def test_big_parallel_equals_sequential_baseline():
+    """At M = 128 (the Fig. 1A model) the parallel solver and its adjoint give the sequential
+    baseline's trajectory, adjoint and gradients."""
+    c = _case(128, 50, 3, 1, 1500, 0.15, 1700)
+    m = oracle_model(c)
+    say("big parallel vs sequential")
+    seq = D.deer_sequential(m, c.x, 0.15, 3)
+    res = D.deer_solve(m, c.x, 0.15, 3, tol=1e-6, max_iter=200)
+    assert res["status"] == 0
+    assert rel_inf(res["z"].cpu().numpy(), seq["z"].cpu().numpy()) < TOL
+    adj = D.deer_adjoint(m, c.x, seq["z"], 0.15, 3)
+    assert rel_inf(adj["lam"].cpu().numpy(), seq["lam"].cpu().numpy()) < TOL
+    for k in ("A", "W1", "W2", "h1", "h2"):
+        assert rel_inf(adj["grads"][k].cpu().numpy(), seq["grads"][k].cpu().numpy()) < TOL, k
+
+
+def test_big_safeguard_reaches_rollout():
+    c = _case(128, 50, 3, 2, 400, 0.15, 1800)
+    m = oracle_model(c)
+    say("big safeguard")
+    res = D.deer_solve(m, c.x, 0.15, 3, tol=1e-5, max_iter=3000, step_bound=0.05)
+    assert res["status"] == 0
+    assert rel_inf(res["z"].cpu().numpy(), O.rollout(m, c.x, 0.15, 3)) < TOL

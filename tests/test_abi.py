@@ -120,11 +120,12 @@ def test_scan_workspace_query_every_orientation(lib):
         for tr in (0, 1):
             assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DENSE, rev, tr, 2, 1000, 32) > 0
             assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DIAG_C64, rev, tr, 2, 1000, 64) > 0
-    assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DENSE, 0, 0, 2, 1000, 65) == 0
+    assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DENSE, 0, 0, 2, 1000, 128) > 0
+    assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DENSE, 0, 0, 2, 1000, 129) == 0
     assert lib.deer_scan_workspace_bytes(_b.DEER_SCAN_DENSE, 0, 0, 0, 1000, 16) == 0
     dummy = (ctypes.c_float * 4)()
     p = ctypes.cast(dummy, ctypes.c_void_p)
-    st = lib.deer_scan(_b.DEER_SCAN_DENSE, 0, 1, 2, 10, 65, p, p, p, None, 0, None)
+    st = lib.deer_scan(_b.DEER_SCAN_DENSE, 0, 1, 2, 10, 129, p, p, p, None, 0, None)
     assert st == _b.DEER_ERR_INVALID_ARG
     st = lib.deer_scan(_b.DEER_SCAN_DENSE, 0, 1, 2, 10, 4, p, p, p, None, 0, None)   # y aliases b
     assert st == _b.DEER_ERR_INVALID_ARG and b"alias" in lib.deer_last_error()

@@ -1741,14 +1741,24 @@ __device__ __forceinline__ float lds_row_dot64(const float (*wl)[68], int row, c
     return a0 + a1;
 }
 
+// M = 64 with a uniform forcing factor (every latent forced, or none): one chain per wave, two
+// waves per SIMD.  J_F = diag(A) + W diag(m) is the matrix-core A operand: W + diag(A) is staged in
+// LDS once, and every step masks its columns with the step's ReLU bits (a column k of W is kept
+// where m_k = 1; the diagonal entry becomes A_k where m_k = 0), one row tile of 16 at a time,
+// shared by the four column tiles.  The chunk product alternates between two accumulator sets
+// (the previous step's set is the unmasked B operand), so no copy, mask or scaling of the
+// accumulators is needed per step; the factor gamma p is applied every 8 steps.  The residual
+// and the chunk-local solution are row dot products against the same LDS rows, corrected for
+// the diagonal: F_i = (W + diag A)_i relu(z~) + A_i min(z~_i, 0), and
+// y_i = (W + diag A)_i (m o u) + A_i u_i (1 - m_i).
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_newton_product_plrnn64u(
     const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
     const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
     const int *__restrict__ zsel, float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout,
     float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
     int ncs) {
-    constexpr int MP = 64, NI = 4, NS = 16;
-    __shared__ __align__(16) float wl[MP][68];
+    constexpr int MP = 64, NI = 4;
+    __shared__ __align__(16) float wl[MP][68];   // W + diag(A), zero padded
     __shared__ __align__(16) float lds[64];
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int id = blockIdx.x;
@@ -1758,20 +1768,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_
     const int len = ok ? min(C, T - s0) : 0;
     for (int e = lane; e < MP * MP; e += 64) {
         const int row = e / MP, col = e % MP;
-        wl[row][col] = (row < M && col < M) ? W[row * M + col] : 0.f;
+        wl[row][col] = (row < M && col < M) ? W[row * M + col] + (row == col ? A[row] : 0.f) : 0.f;
     }
     const float p = N > 0 ? __fsub_rn(1.0f, alpha) : 1.0f;
     const float gp = (gamma ? gamma[b] : 1.f) * p;
     const float gp2 = gp * gp, gp4 = gp2 * gp2, gp8 = gp4 * gp4;
-    float dA[NI][4];
+    // diagonal entries of this lane's A fragments: row 16 I + c is column 16 I + 4 g + q where
+    // c == 4 g + q; there the masked entry is A instead of 0
+    uint32_t dgA[NI][4];
 #pragma unroll
     for (int I = 0; I < NI; ++I)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = 16 * I + 4 * g + r;
-            dA[I][r] = row < M ? A[row] : 0.f;
-        }
-    v4f acc[NI][4];
+        for (int q = 0; q < 4; ++q)
+            dgA[I][q] = (c == 4 * g + q && 16 * I + c < M) ? __float_as_uint(A[16 * I + c]) : 0u;
+    v4f acc[NI][4], acc2[NI][4];
 #pragma unroll
     for (int Jt = 0; Jt < 4; ++Jt)
 #pragma unroll
@@ -1795,9 +1805,42 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_
         zn = z[((size_t)b * T + s0) * M + ui];
         if (forced) xn = x[((size_t)b * (T + 1) + s0) * N + ui];
     }
-    lds_barrier();   // W in LDS
+    lds_barrier();   // W + diag(A) in LDS
     const int maxlen = __builtin_amdgcn_readfirstlane(len);
-    for (int t = 0; t < maxlen; ++t) {
+    // one step of the chain product, from accumulator set `in` to set `out`
+    auto product = [&](const v4f (&in)[NI][4], v4f (&out)[NI][4], uint32_t w0, uint32_t w1) {
+        uint32_t mk[4][4];   // all ones where the ReLU of column 16 j + 4 g + q is on
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                mk[j][q] = (uint32_t)__builtin_amdgcn_sbfe((int)((j >> 1) ? w1 : w0), 16 * (j & 1) + 4 * g + q, 1);
+#pragma unroll
+        for (int I = 0; I < NI; ++I) {
+            float a[4][4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float4 a4 = *reinterpret_cast<const float4 *>(&wl[16 * I + c][16 * j + 4 * g]);
+                const float av[4] = {a4.x, a4.y, a4.z, a4.w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t wb = __float_as_uint(av[q]);
+                    // (m & (W + A delta)) | (~m & A delta): the diagonal tile keeps A where m = 0
+                    a[j][q] = __uint_as_float(j == I ? ((mk[j][q] & wb) | (~mk[j][q] & dgA[I][q])) : (mk[j][q] & wb));
+                }
+            }
+#pragma unroll
+            for (int Jt = 0; Jt < 4; ++Jt) {
+                v4f s = (v4f){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) s = mfma16x16x4(a[j][q], in[j][Jt][q], s);
+                out[I][Jt] = s;
+            }
+        }
+    };
+    auto step = [&](int t, const v4f (&in)[NI][4], v4f (&out)[NI][4]) {
         const bool run = lat;
         const int s = s0 + t;
         const float zcur = zn, xb = xn;
@@ -1814,60 +1857,48 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_
         const uint64_t bal = __ballot(pos);
         lds[lane] = pos ? zt : 0.f;
         lds_barrier();
-        const float F = fmaf(Ai, zt, lds_row_dot64(wl, ui, lds)) + hi;
+        const float F = fmaf(Ai, fminf(zt, 0.f), lds_row_dot64(wl, ui, lds)) + hi;
         lds_barrier();
         const float r = zcur - F;
         if (run) {
             r_out[((size_t)b * T + s) * M + ui] = r;
             if (ui == 0) {
-                const size_t step = (size_t)b * T + s;
-                masks[step * 2] = (uint32_t)bal;
-                if (M > 32) masks[step * 2 + 1] = (uint32_t)(bal >> 32);
+                const size_t stp = (size_t)b * T + s;
+                masks[stp * 2] = (uint32_t)bal;
+                if (M > 32) masks[stp * 2 + 1] = (uint32_t)(bal >> 32);
             }
         }
         // P <- (diag(A) + W diag(m)) P   (the factor gp is applied every 8 steps)
-        const uint32_t w0 = (uint32_t)bal, w1 = (uint32_t)(bal >> 32);
-#pragma unroll
-        for (int Jt = 0; Jt < 4; ++Jt) {
-            float Bop[NS];
-#pragma unroll
-            for (int j = 0; j < NS / 4; ++j) {
-                const uint32_t wj = (j >> 1) ? w1 : w0;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) Bop[4 * j + q] = select_bit(wj, 16 * (j & 1) + 4 * g + q, acc[j][Jt][q]);
-            }
-#pragma unroll
-            for (int I = 0; I < NI; ++I)
-#pragma unroll
-                for (int r2 = 0; r2 < 4; ++r2) acc[I][Jt][r2] *= dA[I][r2];
-#pragma unroll
-            for (int I = 0; I < NI; ++I)
-#pragma unroll
-                for (int j = 0; j < NS / 4; ++j) {
-                    const float4 a4 = *reinterpret_cast<const float4 *>(&wl[16 * I + c][16 * j + 4 * g]);
-                    acc[I][Jt] = mfma16x16x4(a4.x, Bop[4 * j + 0], acc[I][Jt]);
-                    acc[I][Jt] = mfma16x16x4(a4.y, Bop[4 * j + 1], acc[I][Jt]);
-                    acc[I][Jt] = mfma16x16x4(a4.z, Bop[4 * j + 2], acc[I][Jt]);
-                    acc[I][Jt] = mfma16x16x4(a4.w, Bop[4 * j + 3], acc[I][Jt]);
-                }
-        }
+        product(in, out, (uint32_t)bal, (uint32_t)(bal >> 32));
         if ((t & 7) == 7) {
 #pragma unroll
             for (int Jt = 0; Jt < 4; ++Jt)
 #pragma unroll
                 for (int I = 0; I < NI; ++I)
 #pragma unroll
-                    for (int r2 = 0; r2 < 4; ++r2) acc[I][Jt][r2] *= gp8;
+                    for (int r2 = 0; r2 < 4; ++r2) out[I][Jt][r2] *= gp8;
         }
         // chunk-local solution: u <- gp (A o u + W (m o u)) - r
         lds[lane] = pos ? u : 0.f;
         lds_barrier();
-        const float y = fmaf(Ai, u, lds_row_dot64(wl, ui, lds));
+        const float y = fmaf(Ai, pos ? 0.f : u, lds_row_dot64(wl, ui, lds));
         lds_barrier();
         if (run) {
             u = fmaf(gp, y, -r);
             zprev = zcur;
         }
+    };
+    int t = 0;
+    for (; t + 1 < maxlen; t += 2) {
+        step(t, acc, acc2);
+        step(t + 1, acc2, acc);
+    }
+    if (t < maxlen) {   // odd length: the last step lands in the second set
+        step(t, acc, acc2);
+#pragma unroll
+        for (int Jt = 0; Jt < 4; ++Jt)
+#pragma unroll
+            for (int I = 0; I < NI; ++I) acc[I][Jt] = acc2[I][Jt];
     }
     if (ok0 && len > 0) {
         float rest = 1.f;

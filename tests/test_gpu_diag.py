@@ -4,7 +4,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from gpu_util import rel_inf, say
+from gpu_util import rel_inf, say, tie_band_check
 
 pytestmark = pytest.mark.gpu
 
@@ -158,8 +158,7 @@ def test_readout_loss_g_and_grads(B, T, M, H, No):
     out = D.deer_readout_loss(prm, torch.tensor(h), x, want_masks=True)
     got = _bits(out["masks"].cpu().numpy(), H)
     s = O.diag_ssm_readout_preactivation(prm, h)
-    far = np.abs(s) > 1e-5 * max(np.abs(s).max(), 1e-30)
-    assert np.array_equal(got[far], (s > 0)[far])
+    tie_band_check(got, s, 1e-5, "read-out masks")
     loss, g, gr = O.diag_ssm_loss_and_seed(prm, h, x, mask=got)
     assert abs(float(out["loss"].cpu()[0]) - loss) <= 1e-5 * abs(loss)
     assert rel_inf(out["g"].cpu().numpy(), g) < TOL

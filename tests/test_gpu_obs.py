@@ -13,7 +13,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from gpu_util import masks_to_bool, oracle_model, rel_inf, say
+from gpu_util import masks_to_bool, oracle_model, rel_inf, say, tie_band_check
 
 pytestmark = pytest.mark.gpu
 
@@ -50,15 +50,8 @@ def _no_ties(m, zt):
 
 
 def _masks_outside_band(gpu_mask, m, zt, what):
-    """GPU decisions equal the float64 ones wherever |u| > BAND max|u|; returns the in-band count."""
-    u = O.preactivation(m, zt)
-    out = np.abs(u) > BAND * np.abs(u).max()
-    ref = u > 0
-    assert np.array_equal(gpu_mask[out], ref[out]), what
-    nin = int((gpu_mask[~out] != ref[~out]).sum())
-    if nin:
-        print(f"[tie band] {what}: {nin} in-band decisions differ from float64", flush=True)
-    return nin
+    """GPU decisions equal the float64 ones wherever |u| > BAND max|u|, and few differ inside."""
+    return tie_band_check(gpu_mask, O.preactivation(m, zt), BAND, what)
 
 
 CASES = [("plrnn", 5, 0, 2, 2, 60), ("plrnn", 16, 0, 3, 3, 700), ("plrnn", 33, 0, 7, 2, 300),

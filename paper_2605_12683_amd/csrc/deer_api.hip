@@ -436,12 +436,22 @@ struct ShWs {
     NewtonCtl ctl;
 };
 
-static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, bool need_lam, size_t *bytes) {
+// The shallow solve without a stored Jacobian (the forced Jacobians rebuilt from the hidden
+// masks by the chunk product and applied as Jacobian-vector products in the fix-up); on unless
+// DEER_SH_FUSED=0, for the identity read-out at M <= 64 within the kernels' tile limits.
+static bool sh_fused(int M, int L) {
+    const char *e = getenv("DEER_SH_FUSED");
+    if (e && atoi(e) == 0) return false;
+    return shfused_supported(M, L);
+}
+
+static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, bool need_lam, size_t *bytes,
+                     bool stored_J = true) {
     ShWs w{};
     const int LW = (L + 31) / 32;
     Carver c(ws);
     w.masks = c.take<uint32_t>((size_t)B * T * LW);
-    w.J = c.take<float>((size_t)B * T * M * M);
+    w.J = stored_J ? c.take<float>((size_t)B * T * M * M) : nullptr;
     if (op == DEER_OP_SOLVE) {
         const int C = choose_chunk(B, T, padded_dim(M));
         w.ctl = carve_ctl(c, B, (size_t)T * M, (size_t)B * ((T + C - 1) / C));
@@ -919,10 +929,11 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
                          float *final_norm, void *ws, size_t ws_bytes, hipStream_t st) {
     int rc = check_shallow_limits(m);
     if (rc) return rc;
+    const bool fused = sh_fused(m->M, m->L);
     size_t need = 0;
-    carve_sh(nullptr, B, T, m->M, m->L, DEER_OP_SOLVE, false, false, &need);
+    carve_sh(nullptr, B, T, m->M, m->L, DEER_OP_SOLVE, false, false, &need, !fused);
     if ((rc = check_ws(ws, ws_bytes, need))) return rc;
-    ShWs w = carve_sh(ws, B, T, m->M, m->L, DEER_OP_SOLVE, false, false, &need);
+    ShWs w = carve_sh(ws, B, T, m->M, m->L, DEER_OP_SOLVE, false, false, &need, !fused);
     ShArgs a{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
     if ((rc = init_guess(o, B, T, m->M, f->n_forced, x, z, st))) return rc;
     std::vector<int> act(B, 1), it(B, 0);
@@ -933,6 +944,13 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
                       uint32_t) -> int {
         int r;
         if ((r = launch_resjac_shplrnn(a, zb, za, zsel, nullptr, w.r, w.masks, dact, st))) return r;
+        if (fused) {
+            if ((r = launch_chunk_product_shfused(a, w.masks, w.r, -1.f, gam, d.P, d.v, dact, d.C, d.ncs, st)))
+                return r;
+            if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nullptr, B, d.ncs, d.gws, st))) return r;
+            return launch_fixup_shjvp(a, w.masks, w.r, -1.f, gam, d.carry, zb, za, zsel, w.ctl.chain_bits, dact, d.C,
+                                      d.ncs, st);
+        }
         if ((r = launch_jacform_shplrnn(a, w.masks, w.J, dact, gam, st))) return r;
         if ((r = launch_chunk_product_dense(false, B, T, m->M, w.J, w.r, -1.f, d.P, d.v, dact, d.C, d.ncs, st))) return r;
         if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nullptr, B, d.ncs, d.gws, st))) return r;
@@ -1454,7 +1472,8 @@ size_t deer_workspace_bytes(const deer_model *m, int B, int T, int op) {
     }
     if (m->kind == DEER_SHPLRNN) {
         size_t bytes = 0;
-        carve_sh(nullptr, B, T, m->M, m->L, op, true, true, &bytes);
+        carve_sh(nullptr, B, T, m->M, m->L, op, true, true, &bytes,
+                 !(op == DEER_OP_SOLVE && sh_fused(m->M, m->L)));
         return bytes;
     }
     return 0;

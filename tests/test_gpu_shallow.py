@@ -144,3 +144,38 @@ def test_config3_reduced():
     assert rel_inf(out["lam"].cpu().numpy(), lam) < TOL
     for k in ("A", "W1", "W2", "h1", "h2"):
         assert rel_inf(out["grads"][k].cpu().numpy(), gr[k]) < TOL, k
+
+
+@pytest.mark.parametrize("M,L,N,B,T,alpha,chunk", [(32, 256, 32, 3, 700, 0.1, 0), (32, 256, 8, 2, 1000, 0.1, 37),
+                                                   (5, 20, 2, 2, 333, 0.3, 33), (16, 384, 16, 2, 300, 0.1, 0),
+                                                   (64, 128, 64, 2, 257, 0.1, 0), (64, 50, 3, 1, 400, 0.15, 0),
+                                                   (1, 7, 1, 2, 50, 0.2, 0), (24, 48, 24, 3, 129, 0.2, 16),
+                                                   (40, 100, 10, 5, 211, 0.2, 0)])
+def test_shallow_fused_and_stored_updates_agree(M, L, N, B, T, alpha, chunk):
+    """The Newton update without a stored Jacobian (J~_t rebuilt from the hidden masks inside
+    the chunk product, Jacobian-vector products in the fix-up) and the stored-Jacobian update
+    both reach the sequential rollout, in the same number of updates up to one (the two round
+    differently); with forced rejections (damped gamma J~) as well.  Covers ragged last chunks,
+    sequences that converge at different updates, and every register-tile variant."""
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    c = _case(M, L, N, B, T, alpha, 900 + M + L)
+    m = oracle_model(c)
+    ref = O.rollout(m, c.x, alpha, N)
+    out = {}
+    try:
+        for path in ("0", "1"):
+            os.environ["DEER_SH_FUSED"] = path
+            say("deer_solve shallow path", path, M, L, N, B, T, alpha, chunk)
+            res = D.deer_solve(m, c.x, alpha, N, tol=1e-5, max_iter=200)
+            assert res["status"] == 0, (path, res)
+            assert rel_inf(res["z"].cpu().numpy(), ref) < TOL, path
+            say("deer_solve shallow path with rejections", path)
+            rj = D.deer_solve(m, c.x, alpha, N, tol=1e-5, max_iter=5000, step_bound=0.05)
+            assert rj["status"] == 0, (path, rj)
+            assert rel_inf(rj["z"].cpu().numpy(), ref) < TOL, path
+            out[path] = (list(res["iters"]), list(rj["iters"]))
+    finally:
+        os.environ.pop("DEER_SH_FUSED", None)
+    for a, b in zip(out["0"][0], out["1"][0]):
+        assert abs(a - b) <= 1, out

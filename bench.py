@@ -109,13 +109,11 @@ def _diag_step(D, model, readout, xd, c, ws_s, ws_r, ws_a, bufs):
     return c.B
 
 
-def kernel_work(c, steps, updates, fwd_rows=None, sh_fused=False):
+def kernel_work(c, steps, updates, fwd_rows=None):
     """Algorithmic work of each kernel over the timed region: {name: (bound, total work)};
     work in flop (mfma) or bytes (hbm).  `updates` = Newton updates summed over sequences;
     `fwd_rows` (latent warm-up) = the (b, t) steps those updates covered, when an update does
-    not span the whole sequence; `sh_fused`: the shallow solve ran without a stored Jacobian
-    (k_chunk_product_shfused + k_fixup_shjvp), so the stored-Jacobian kernels served the adjoint
-    only."""
+    not span the whole sequence."""
     B, T, M, N = c.B, c.T, c.M, c.n_obs
     W = (M + 31) // 32
     fwd = updates * T if fwd_rows is None else fwd_rows   # (b, t) steps processed by the updates
@@ -168,13 +166,16 @@ def kernel_work(c, steps, updates, fwd_rows=None, sh_fused=False):
     else:
         L = c.L
         LW = (L + 31) // 32
-        stored = adj if sh_fused else fwd + adj
-        out["k_jacform_shplrnn"] = ("mfma", stored * 2.0 * M * M * L)
-        out["k_chunk_product_dense"] = ("mfma", (prod - fwd if sh_fused else prod) * 2.0 * M ** 3)
-        # the solve without a stored Jacobian: J~_t formed (2 M^2 L) and composed (2 M^3) in the
-        # chunk product; two matrix-vector products with W2 and W1 (4 M L) per step in the fix-up
+        out["k_jacform_shplrnn"] = ("mfma", (fwd + adj) * 2.0 * M * M * L)
+        out["k_chunk_product_dense"] = ("mfma", prod * 2.0 * M ** 3)
+        # without a stored Jacobian: J~_t formed (2 M^2 L) and composed (2 M^3) in the chunk
+        # products; two matrix-vector products with W1 and W2 (4 M L) per step in the fix-ups
         out["k_chunk_product_shfused"] = ("mfma", fwd * (2.0 * M * M * L + 2.0 * M ** 3))
+        out["k_chunk_product_shfused_rev"] = ("mfma", steps * B * (T - 1) * (2.0 * M * M * L + 2.0 * M ** 3))
         out["k_fixup_shjvp"] = ("mfma", fwd * 4.0 * M * L)
+        # the Newton passes' residual on the matrix cores: u = W2 z~ and W1 relu(u), 4 M L per step
+        out["k_resjac_shmfma"] = ("mfma", fwd * 4.0 * M * L)
+        out["k_fixup_shjvp_rev"] = ("mfma", steps * B * (T - 1) * 4.0 * M * L)
         out["k_resjac_shplrnn"] = ("hbm", (fwd + adj) * (8 * M + 4 * N + 4 * LW))
         out["k_fixup_dense_fwd"] = ("hbm", fwd * (4 * M * M + 12 * M))
         out["k_fixup_dense_rev"] = ("hbm", adj * (4 * M * M + 8 * M))
@@ -185,7 +186,8 @@ def kernel_work(c, steps, updates, fwd_rows=None, sh_fused=False):
 # scaled by the reading of a plain copy of known size in the same run; kept in
 # profiles/traffic_<workload>.txt together with the hash of the kernel's source file, and
 # reported only while that source is unchanged.
-KERNEL_SOURCE = {"k_chunk_product_shfused": "k_shfused.hip", "k_fixup_shjvp": "k_shfused.hip", "k_newton_product_plrnn": "k_plrnn.hip", "k_newton_pass16": "k_plrnn.hip", "k_chunk_product_plrnn": "k_plrnn.hip",
+KERNEL_SOURCE = {"k_chunk_product_shfused": "k_shfused.hip", "k_chunk_product_shfused_rev": "k_shfused.hip",
+                 "k_fixup_shjvp": "k_shfused.hip", "k_resjac_shmfma": "k_shfused.hip", "k_newton_product_plrnn": "k_plrnn.hip", "k_newton_pass16": "k_plrnn.hip", "k_chunk_product_plrnn": "k_plrnn.hip",
                  "k_fixup_fwd_plrnn": "k_plrnn.hip", "k_jacform_shplrnn": "k_shallow.hip",
                  "k_chunk_product_dense": "k_dense.hip", "k_readout": "k_readout.hip",
                  "k_diag_scan_lb_grads": "k_diag.hip", "k_diag_seg_write": "k_diag.hip",
@@ -236,9 +238,9 @@ def measured_mfma(workload, kernel):
             "source": f"profiles/mfma_{workload}.txt"}
 
 
-def roofline_for(name, c, total_ms, launches, steps, updates, fwd_rows=None, sh_fused=False):
+def roofline_for(name, c, total_ms, launches, steps, updates, fwd_rows=None):
     """Algorithmic work of the dominant kernel over the timed region, divided by its time."""
-    work = kernel_work(c, steps, updates, fwd_rows, sh_fused)
+    work = kernel_work(c, steps, updates, fwd_rows)
     base = {"kernel": name, "avg_launch_ms": total_ms / launches, "launches": launches,
             "traffic": measured_traffic(c.name, name)}
     if name not in work:
@@ -557,10 +559,9 @@ def main():
     modeled = {k: v for k, v in kt.items() if k in kernel_work(c, 1, 1)}
     dom = max((modeled or kt).items(), key=lambda kv: kv[1][0])
     prof_rows = rows_of(prof_updates, prof_steps)
-    shf = "k_chunk_product_shfused" in kt
-    roof = roofline_for(dom[0], c, dom[1][0], dom[1][1], prof_steps, prof_updates, prof_rows, shf)
+    roof = roofline_for(dom[0], c, dom[1][0], dom[1][1], prof_steps, prof_updates, prof_rows)
     kernels = {k: {"ms_total": ms, "launches": n, **({"frac": r["frac"], "unit": r["unit"], "achieved": r["achieved"]}
-                                                      if (r := roofline_for(k, c, ms, n, prof_steps, prof_updates, prof_rows, shf))["frac"]
+                                                      if (r := roofline_for(k, c, ms, n, prof_steps, prof_updates, prof_rows))["frac"]
                                                       is not None else {})}
                for k, (ms, n) in kt.items()}
 

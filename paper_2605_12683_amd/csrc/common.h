@@ -93,6 +93,25 @@ __device__ __forceinline__ float *next_iter(float *z, float *zalt, const int *zs
     return (zsel && zsel[b]) ? z : zalt;
 }
 
+// (sequence, step) of the rows row0 + rr of a [B, T] row space: the first row's pair from one
+// division per tile, the others by carrying over sequence ends (rr small), instead of a 64-bit
+// division per row
+struct RowBase {
+    int b0, s0;
+};
+__device__ __forceinline__ RowBase row_base(long row0, int T) {
+    const long b = row0 / T;
+    return {(int)b, (int)(row0 - b * T)};
+}
+__device__ __forceinline__ void row_at(RowBase rb, int rr, int T, int &b, int &s) {
+    s = rb.s0 + rr;
+    b = rb.b0;
+    while (s >= T) {
+        s -= T;
+        ++b;
+    }
+}
+
 // Workgroup barrier that orders LDS only: unlike __syncthreads it does not wait for
 // outstanding global loads, so loads issued ahead (prefetch) stay in flight across it.  For
 // kernels whose threads exchange data through LDS alone.

@@ -298,7 +298,9 @@ static bool pass_fusion_allowed() {
 // Chunk length of the dense scans: enough chains to fill the machine (about 2048 waves),
 // and a bounded number of chunks per sequence so that the two-level carry pass stays short
 // (1024 for MP <= 32, 512 for MP = 64, whose group pass composes 64 x 64 maps).
-static int choose_chunk(int B, int T, int MP) {
+// sh_fused: the shallow update without a stored Jacobian, whose fix-up runs 16 chains per block
+// (8192 chains keep two of its waves on every SIMD)
+static int choose_chunk(int B, int T, int MP, bool sh_fused = false) {
     const int ov = chunk_override();
     if (ov > 0) return ov < T ? ov : T;
     const long total = (long)B * T;
@@ -313,7 +315,7 @@ static int choose_chunk(int B, int T, int MP) {
         if (C > T) C = T;
         return (int)C;
     }
-    const long target_chains = MP == 64 ? 8192L : 2048L * (64 / MP);
+    const long target_chains = (MP == 64 || sh_fused) ? 8192L : 2048L * (64 / MP);
     long C = (total + target_chains - 1) / target_chains;
     if (C < 16) C = 16;
     const long maxc = MP <= 32 ? 1024 : 512;
@@ -414,10 +416,10 @@ struct DenseWs {
     int C, ncs, MP;
 };
 
-static DenseWs carve_dense(void *ws, int B, int T, int M, size_t *bytes) {
+static DenseWs carve_dense(void *ws, int B, int T, int M, size_t *bytes, bool sh_fused = false) {
     DenseWs w{};
     w.MP = padded_dim(M);
-    w.C = choose_chunk(B, T, w.MP);
+    w.C = choose_chunk(B, T, w.MP, sh_fused);
     w.ncs = (T + w.C - 1) / w.C;
     const size_t nch = (size_t)B * w.ncs;
     Carver c(ws);
@@ -436,13 +438,21 @@ struct ShWs {
     NewtonCtl ctl;
 };
 
-// The shallow solve without a stored Jacobian (the forced Jacobians rebuilt from the hidden
-// masks by the chunk product and applied as Jacobian-vector products in the fix-up); on unless
-// DEER_SH_FUSED=0, for the identity read-out at M <= 64 within the kernels' tile limits.
+// The shallow solve and adjoint without a stored Jacobian (the forced Jacobians rebuilt from the
+// hidden masks by the chunk products and applied as Jacobian-vector products in the fix-ups); on
+// unless DEER_SH_FUSED=0, for the identity read-out at M <= 64 within the kernels' tile limits.
 static bool sh_fused(int M, int L) {
     const char *e = getenv("DEER_SH_FUSED");
     if (e && atoi(e) == 0) return false;
     return shfused_supported(M, L);
+}
+
+// Newton passes of the fused shallow path: residual and masks on the matrix cores (the pass's
+// own masks; the fixed-order float32 decision of k_resjac_shplrnn is kept for the masks a
+// caller receives and for the adjoint); on unless DEER_SH_RESMFMA=0
+static bool sh_res_mfma() {
+    const char *e = getenv("DEER_SH_RESMFMA");
+    return !e || atoi(e) != 0;
 }
 
 static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, bool need_lam, size_t *bytes,
@@ -453,7 +463,7 @@ static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, 
     w.masks = c.take<uint32_t>((size_t)B * T * LW);
     w.J = stored_J ? c.take<float>((size_t)B * T * M * M) : nullptr;
     if (op == DEER_OP_SOLVE) {
-        const int C = choose_chunk(B, T, padded_dim(M));
+        const int C = choose_chunk(B, T, padded_dim(M), !stored_J);
         w.ctl = carve_ctl(c, B, (size_t)T * M, (size_t)B * ((T + C - 1) / C));
         w.r = c.take<float>((size_t)B * T * M);
     } else {
@@ -463,7 +473,7 @@ static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, 
         w.part = c.take<float>(sh_grads_part_floats(M, L, &nb));
     }
     size_t dbytes = 0;
-    w.d = carve_dense(ws ? (char *)ws + c.off : nullptr, B, T, M, &dbytes);
+    w.d = carve_dense(ws ? (char *)ws + c.off : nullptr, B, T, M, &dbytes, !stored_J);
     *bytes = c.off + dbytes;
     return w;
 }
@@ -943,13 +953,17 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
     auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *,
                       uint32_t) -> int {
         int r;
-        if ((r = launch_resjac_shplrnn(a, zb, za, zsel, nullptr, w.r, w.masks, dact, st))) return r;
+        if (fused && sh_res_mfma()) {
+            if ((r = launch_resjac_shmfma(a, zb, za, zsel, w.r, w.masks, dact, st))) return r;
+        } else if ((r = launch_resjac_shplrnn(a, zb, za, zsel, nullptr, w.r, w.masks, dact, st))) {
+            return r;
+        }
         if (fused) {
-            if ((r = launch_chunk_product_shfused(a, w.masks, w.r, -1.f, gam, d.P, d.v, dact, d.C, d.ncs, st)))
+            if ((r = launch_chunk_product_shfused(false, a, w.masks, w.r, -1.f, gam, d.P, d.v, dact, d.C, d.ncs, st)))
                 return r;
             if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nullptr, B, d.ncs, d.gws, st))) return r;
-            return launch_fixup_shjvp(a, w.masks, w.r, -1.f, gam, d.carry, zb, za, zsel, w.ctl.chain_bits, dact, d.C,
-                                      d.ncs, st);
+            return launch_fixup_shjvp(false, a, w.masks, w.r, -1.f, gam, d.carry, zb, za, zsel, w.ctl.chain_bits, dact,
+                                      d.C, d.ncs, st);
         }
         if ((r = launch_jacform_shplrnn(a, w.masks, w.J, dact, gam, st))) return r;
         if ((r = launch_chunk_product_dense(false, B, T, m->M, w.J, w.r, -1.f, d.P, d.v, dact, d.C, d.ncs, st))) return r;
@@ -1472,8 +1486,7 @@ size_t deer_workspace_bytes(const deer_model *m, int B, int T, int op) {
     }
     if (m->kind == DEER_SHPLRNN) {
         size_t bytes = 0;
-        carve_sh(nullptr, B, T, m->M, m->L, op, true, true, &bytes,
-                 !(op == DEER_OP_SOLVE && sh_fused(m->M, m->L)));
+        carve_sh(nullptr, B, T, m->M, m->L, op, true, true, &bytes, !sh_fused(m->M, m->L));
         return bytes;
     }
     return 0;
@@ -1628,10 +1641,11 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
     }
     if (m->kind == DEER_SHPLRNN) {
         if ((rc = check_shallow_limits(m))) return rc;
+        const bool fused = sh_fused(m->M, m->L);
         size_t need = 0;
-        carve_sh(nullptr, B, T, m->M, m->L, DEER_OP_ADJOINT, true, true, &need);
+        carve_sh(nullptr, B, T, m->M, m->L, DEER_OP_ADJOINT, true, true, &need, !fused);
         if ((rc = check_ws(ws, ws_bytes, need))) return rc;
-        ShWs w = carve_sh(ws, B, T, m->M, m->L, DEER_OP_ADJOINT, true, true, &need);
+        ShWs w = carve_sh(ws, B, T, m->M, m->L, DEER_OP_ADJOINT, true, true, &need, !fused);
         ShArgs a{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
         const DenseWs &d = w.d;
         const float *gg = g;
@@ -1642,10 +1656,23 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
         }
         float *lo = lam ? lam : w.lam;
         if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, nullptr, nullptr, w.masks, nullptr, st))) return rc;
-        if ((rc = launch_jacform_shplrnn(a, w.masks, w.J, nullptr, nullptr, st))) return rc;
-        if ((rc = launch_chunk_product_dense(true, B, T, m->M, w.J, gg, 1.f, d.P, d.v, nullptr, d.C, d.ncs, st))) return rc;
-        if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, d.gws, st))) return rc;
-        if ((rc = launch_fixup_dense(2, B, T, m->M, w.J, gg, 1.f, d.carry, nullptr, lo, nullptr, nullptr, nullptr, d.C, d.ncs, st))) return rc;
+        if (fused) {
+            if ((rc = launch_chunk_product_shfused(true, a, w.masks, gg, 1.f, nullptr, d.P, d.v, nullptr, d.C, d.ncs,
+                                                   st)))
+                return rc;
+            if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, d.gws, st))) return rc;
+            if ((rc = launch_fixup_shjvp(true, a, w.masks, gg, 1.f, nullptr, d.carry, nullptr, lo, nullptr, nullptr,
+                                         nullptr, d.C, d.ncs, st)))
+                return rc;
+        } else {
+            if ((rc = launch_jacform_shplrnn(a, w.masks, w.J, nullptr, nullptr, st))) return rc;
+            if ((rc = launch_chunk_product_dense(true, B, T, m->M, w.J, gg, 1.f, d.P, d.v, nullptr, d.C, d.ncs, st)))
+                return rc;
+            if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, d.gws, st))) return rc;
+            if ((rc = launch_fixup_dense(2, B, T, m->M, w.J, gg, 1.f, d.carry, nullptr, lo, nullptr, nullptr, nullptr,
+                                         d.C, d.ncs, st)))
+                return rc;
+        }
         if (grads && (grads->A || grads->W || grads->W2 || grads->h || grads->h2)) {
             if ((rc = launch_grads_shplrnn(a, z, lo, w.masks, w.part, grads, st))) return rc;
         }

@@ -63,10 +63,13 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
     // elements whose residual it writes at the end of the tile
     const int rc = tid / (MP / 4), i0 = 4 * (tid % (MP / 4));
     float pz[4], px[4], pc[4], cz[4];   // z_{s-1} (or the initial state at s = 0), x_s, z_s
+    bool plater = false;                // the fetched row exists and has s > 0
     auto fetch = [&](long tile) {
         const long row = tile * TT + rc;
         const bool ok = tid < NT4 && tile < ntiles && row < total;
-        const int b = ok ? (int)(row / T) : 0, s = ok ? (int)(row % T) : 0;
+        int b = 0, s = 0;
+        if (ok) row_at(row_base(tile * TT, T), rc, T, b, s);
+        plater = ok && s > 0;
         const float *z = cur_iter(zbuf, zalt, zsel, b);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -103,8 +106,7 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
         const long row0 = tile * TT;
         __syncthreads();   // the previous tile is done with zT, zc, ru and red
         if (tid < NT4) {
-            const long row = row0 + rc;
-            const bool later = row < total && (int)(row % T) > 0;
+            const bool later = plater;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int i = i0 + r;
@@ -116,7 +118,9 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
         }
         if (tid < TT) {
             const long row = row0 + tid;
-            rowok[tid] = row < total && (!active || active[row / T]);
+            int b = 0, sr = 0;
+            if (row < total) row_at(row_base(row0, T), tid, T, b, sr);
+            rowok[tid] = row < total && (!active || active[b]);
         }
         fetch(tile + gridDim.x);
         __syncthreads();

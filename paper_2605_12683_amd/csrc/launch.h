@@ -187,12 +187,15 @@ int launch_grads_big(const ShArgs &a, const float *z, const float *lam, const ui
 // shallow PLRNN Newton update without a stored Jacobian (masks + W1, W2 only)
 bool shfused_supported(int M, int L);
 size_t shfused_product_lds(int M, int L);
-int launch_chunk_product_shfused(const ShArgs &a, const uint32_t *masks, const float *rhs, float rhs_sign,
-                                 const float *gamma, float *P, float *v, const int *active, int C, int ncs,
-                                 hipStream_t st);
-int launch_fixup_shjvp(const ShArgs &a, const uint32_t *masks, const float *rhs, float rhs_sign, const float *gamma,
-                       const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
-                       const int *active, int C, int ncs, hipStream_t st);
+int launch_resjac_shmfma(const ShArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
+                         uint32_t *masks, const int *active, hipStream_t st);
+// rev: the adjoint's reverse recursion (gamma and active must be null; the fix-up writes y to out)
+int launch_chunk_product_shfused(bool rev, const ShArgs &a, const uint32_t *masks, const float *rhs,
+                                 float rhs_sign, const float *gamma, float *P, float *v, const int *active, int C,
+                                 int ncs, hipStream_t st);
+int launch_fixup_shjvp(bool rev, const ShArgs &a, const uint32_t *masks, const float *rhs, float rhs_sign,
+                       const float *gamma, const float *carry_in, float *z, float *out, const int *zsel,
+                       uint32_t *chain_bits, const int *active, int C, int ncs, hipStream_t st);
 size_t sh_resjac_lds(int M, int L);
 size_t sh_jacform_lds(int M, int L);
 size_t sh_grads_part_floats(int M, int L, int *nblocks);

@@ -152,20 +152,28 @@ def test_config3_reduced():
                                                    (1, 7, 1, 2, 50, 0.2, 0), (24, 48, 24, 3, 129, 0.2, 16),
                                                    (40, 100, 10, 5, 211, 0.2, 0)])
 def test_shallow_fused_and_stored_updates_agree(M, L, N, B, T, alpha, chunk):
-    """The Newton update without a stored Jacobian (J~_t rebuilt from the hidden masks inside
-    the chunk product, Jacobian-vector products in the fix-up) and the stored-Jacobian update
-    both reach the sequential rollout, in the same number of updates up to one (the two round
-    differently); with forced rejections (damped gamma J~) as well.  Covers ragged last chunks,
+    """The Newton update and the adjoint without a stored Jacobian (J~_t rebuilt from the
+    hidden masks inside the chunk products, Jacobian-vector products in the fix-ups) and the
+    stored-Jacobian ones: both solves reach the sequential rollout, in the same number of
+    updates up to one (the two round differently), also with forced rejections (damped gamma
+    J~); both adjoints and all gradients equal the oracle's.  Covers ragged last chunks,
     sequences that converge at different updates, and every register-tile variant."""
     if chunk:
         os.environ["DEER_CHUNK"] = str(chunk)
     c = _case(M, L, N, B, T, alpha, 900 + M + L)
     m = oracle_model(c)
     ref = O.rollout(m, c.x, alpha, N)
+    z32 = ref.astype(np.float32)
+    lam = O.adjoint(m, c.x, z32, alpha, N, mask_precision="float32")
+    gr = O.param_grads(m, c.x, z32, alpha, N, lam, mask_precision="float32")
     out = {}
+    # stored J~; without a stored J~ and the fixed-order residual; the default (matrix-core
+    # residual in the Newton passes)
+    paths = {"0": ("0", "1"), "1x": ("1", "0"), "1": ("1", "1")}
     try:
-        for path in ("0", "1"):
-            os.environ["DEER_SH_FUSED"] = path
+        for path, (fz, rm) in paths.items():
+            os.environ["DEER_SH_FUSED"] = fz
+            os.environ["DEER_SH_RESMFMA"] = rm
             say("deer_solve shallow path", path, M, L, N, B, T, alpha, chunk)
             res = D.deer_solve(m, c.x, alpha, N, tol=1e-5, max_iter=200)
             assert res["status"] == 0, (path, res)
@@ -175,7 +183,14 @@ def test_shallow_fused_and_stored_updates_agree(M, L, N, B, T, alpha, chunk):
             assert rj["status"] == 0, (path, rj)
             assert rel_inf(rj["z"].cpu().numpy(), ref) < TOL, path
             out[path] = (list(res["iters"]), list(rj["iters"]))
+            say("deer_adjoint shallow path", path)
+            adj = D.deer_adjoint(m, c.x, z32, alpha, N)
+            assert rel_inf(adj["lam"].cpu().numpy(), lam) < TOL, path
+            for k in ("A", "W1", "W2", "h1", "h2"):
+                assert rel_inf(adj["grads"][k].cpu().numpy(), gr[k]) < TOL, (path, k)
     finally:
         os.environ.pop("DEER_SH_FUSED", None)
-    for a, b in zip(out["0"][0], out["1"][0]):
-        assert abs(a - b) <= 1, out
+        os.environ.pop("DEER_SH_RESMFMA", None)
+    for p2 in ("1x", "1"):
+        for a, b in zip(out["0"][0], out[p2][0]):
+            assert abs(a - b) <= 1, out

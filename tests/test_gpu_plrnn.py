@@ -151,6 +151,35 @@ def test_fused_and_separate_pass_kernels_agree(M, N, B, T, alpha, chunk, bound):
     assert max(abs(a - b) for a, b in zip(out["1"], out["0"])) <= 1
 
 
+@pytest.mark.parametrize("M,N,B,T,alpha,chunk,bound", [(64, 64, 3, 2000, 0.1, 0, 0.0), (64, 32, 2, 777, 0.2, 0, 0.0),
+                                                         (33, 5, 2, 513, 0.2, 37, 0.0), (20, 20, 5, 300, 0.2, 0, 0.0),
+                                                         (48, 7, 2, 700, 0.15, 64, 0.05), (61, 61, 17, 129, 0.1, 16, 0.0)])
+def test_fixup_matrix_core_and_vector_paths_agree(M, N, B, T, alpha, chunk, bound):
+    """M in 17..64: the forward fix-up on the matrix cores (16 chains as columns, W diag(p) row
+    tiles per wave, Delta through LDS) and the lane-per-latent one both reach the rollout, in the
+    same number of updates up to one; ragged chunks, M not a multiple of 4, many sequences
+    converging at different updates, and forced rejections (damped gamma J~)."""
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    c = _case(M, N, B, T, alpha, 5100 + M + B)
+    m = oracle_model(c)
+    ref = O.rollout(m, c.x, alpha, N)
+    its = {}
+    try:
+        for path in ("0", "1"):
+            os.environ["DEER_FIX_MFMA"] = path
+            say("fixup path", path, M, N, B, T, alpha, chunk, bound)
+            res = D.deer_solve(m, c.x, alpha, N, tol=1e-5, max_iter=3000, step_bound=bound)
+            assert res["status"] == 0, (path, res)
+            assert rel_inf(res["z"].cpu().numpy(), ref) < TOL, path
+            its[path] = list(res["iters"])
+    finally:
+        os.environ.pop("DEER_FIX_MFMA", None)
+    if bound == 0.0:
+        for a, b in zip(its["0"], its["1"]):
+            assert abs(a - b) <= 1, its
+
+
 @pytest.mark.parametrize("M,N,B,T,alpha,chunk,bound", [(16, 3, 4, 300, 0.2, 0, 0.05), (16, 3, 3, 300, 0.2, 16, 0.3),
                                                        (32, 8, 3, 300, 0.1, 16, 0.1), (64, 64, 2, 200, 0.05, 0, 0.1),
                                                        (5, 2, 5, 120, 0.3, 7, 0.02), (16, 3, 3, 512, 0.2, 16, 0.3)])

@@ -640,33 +640,76 @@ __global__ __launch_bounds__(256) void k_resjac_shmfma(const ShArgs a, const flo
     const long total = (long)a.B * T;
     const long ntiles = (total + 15) / 16;
     const long nw = (long)gridDim.x * 4;
-    for (long tile = (long)blockIdx.x * 4 + wv; tile < ntiles; tile += nw) {
+    // The inputs of a tile for row c, latents i = 16j + 4g + q: z_{s-1} (or the initial state at
+    // s = 0) and x_s, combined into z~ as k_resjac_shplrnn does, and z_s.  Every lane loads from a
+    // valid address (rows past the end, inactive sequences and latents past M read row 0 /
+    // latent 0 and are zeroed after), so the loads carry no branches and the next tile's, issued
+    // at the top of a tile, are waited for only when the tile ends.
+    struct RowIn {   // (sequence, step) of row c of a tile and the sequence's control words
+        int b, s, sel, act;
+        bool inr;
+    };
+    struct TileIn {
+        float zp[NI][4], xs[NI][4], zc[NI][4];
+        int s;
+        bool ok;
+    };
+    // stage 1, two tiles ahead: the row's position and its control words (loads in flight)
+    auto rowin = [&](long tile, RowIn &ri) {
         const long rowc = tile * 16 + c;
-        int b = 0, s = 0;
-        if (rowc < total) row_at(row_base(tile * 16, T), c, T, b, s);
-        const bool rok = rowc < total && (!active || active[b]);
-        // z~ and z of row c at the latents i = 16j + 4g + q (the B layout of the first product
-        // and the accumulator layout of F alike)
-        const float *z = cur_iter(zbuf, zalt, zsel, b);
+        ri.b = 0;
+        ri.s = 0;
+        ri.inr = tile < ntiles && rowc < total;
+        if (ri.inr) row_at(row_base(tile * 16, T), c, T, ri.b, ri.s);
+        ri.sel = zsel ? zsel[ri.b] : 0;
+        ri.act = active ? active[ri.b] : 1;
+    };
+    // stage 2, one tile ahead: the inputs, at addresses from the control words loaded a tile ago
+    auto fetch = [&](const RowIn &ri, TileIn &in) {
+        const int b = ri.b, s = ri.s;
+        in.ok = ri.inr && ri.act != 0;
+        in.s = s;
+        const float *z = ri.sel ? zalt : zbuf;
+        const size_t rp = (size_t)b * T + (s > 0 ? s - 1 : 0), rc = (size_t)b * T + s;
+        const size_t xr = ((size_t)b * (T + 1) + s) * (size_t)(N > 0 ? N : 1);
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int i = 16 * j + 4 * g + q, ic = i < M ? i : 0;
+                const float zpv = z[rp * M + ic];
+                const float z0v = a.z0 ? a.z0[(size_t)b * M + ic] : 0.f;
+                in.zp[j][q] = s > 0 ? zpv : z0v;
+                in.xs[j][q] = N > 0 ? a.x[xr + (i < N ? i : 0)] : 0.f;
+                in.zc[j][q] = z[rc * M + ic];
+            }
+    };
+    const long t0w = (long)blockIdx.x * 4 + wv;
+    RowIn r1, r2;
+    TileIn cur, nxt;
+    rowin(t0w, r1);
+    fetch(r1, cur);
+    rowin(t0w + nw, r1);
+    for (long tile = t0w; tile < ntiles; tile += nw) {
+        rowin(tile + 2 * nw, r2);
+        fetch(r1, nxt);
+        const long rowc = tile * 16 + c;
+        const bool rok = cur.ok;
+        const int s = cur.s;
         float zt[NI][4], zc[NI][4];
 #pragma unroll
         for (int j = 0; j < NI; ++j)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int i = 16 * j + 4 * g + q;
-                float v = 0.f, cur = 0.f;
-                if (rok && i < M) {
-                    if (s == 0) {
-                        v = a.z0 ? a.z0[(size_t)b * M + i] : (i < N ? a.x[(size_t)b * (T + 1) * N + i] : 0.f);
-                    } else {
-                        const float zp = z[((size_t)b * T + s - 1) * M + i];
-                        v = i < N ? __fadd_rn(__fmul_rn(p, zp), __fmul_rn(a.alpha, a.x[((size_t)b * (T + 1) + s) * N + i]))
-                                  : zp;
-                    }
-                    cur = z[(size_t)rowc * M + i];
-                }
-                zt[j][q] = v;
-                zc[j][q] = cur;
+                float v;
+                if (s == 0)   // the initial state: z0, or [x_0; 0]
+                    v = a.z0 ? cur.zp[j][q] : (i < N ? cur.xs[j][q] : 0.f);
+                else
+                    v = i < N ? __fadd_rn(__fmul_rn(p, cur.zp[j][q]), __fmul_rn(a.alpha, cur.xs[j][q])) : cur.zp[j][q];
+                const bool e = rok && i < M;
+                zt[j][q] = e ? v : 0.f;
+                zc[j][q] = e ? cur.zc[j][q] : 0.f;
             }
         v4f F[NI];
 #pragma unroll
@@ -715,6 +758,8 @@ __global__ __launch_bounds__(256) void k_resjac_shmfma(const ShArgs a, const flo
                     if (i < M) r_out[(size_t)rowc * M + i] = zc[I][r] - (fmaf(dA[I][r], zt[I][r], F[I][r]) + h1v[I][r]);
                 }
         }
+        cur = nxt;
+        r1 = r2;
     }
 }
 

@@ -12,7 +12,8 @@ One step = one pass of the whole path over one batch of synthetic input:
                    with conj(lambda) + dlambda / dBc reductions).
 Inputs are resident in HBM before the timed region.  The value is DEER timesteps per
 second: sum over sequences of T x Newton updates, per second of the whole step (with a latent
-warm-up, --tw, an update is counted at the length of the part it covered: T_w or T - T_w).
+warm-up, --tw, where the library chains a solve of steps 1..T_w and one of the rest, an update
+is counted at the length of the part it covered: T_w or T - T_w).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 5]
 
@@ -56,6 +57,12 @@ def _plrnn_step(D, model, xd, c, ws_s, ws_a, T_w=0):
     # the step's outputs are the parameter gradients: the adjoint itself is not stored
     D.deer_adjoint(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a, want_lam=False, T_w=T_w)
     return sum(res["iters"])
+
+
+def warmup_in_one_iteration(kind, M, quasi):
+    """The library runs the latent warm-up inside the one Newton iteration for the vanilla PLRNN
+    with M <= 16 (GTF-DEER, identity read-out); elsewhere it chains two solves."""
+    return kind == "plrnn" and M <= 16 and not quasi
 
 
 def update_rows(T, T_w, updates, warm_updates, nsteps):
@@ -505,11 +512,13 @@ def main():
         print(f"workload {c.name}: model kind {c.kind} not supported by this build", file=sys.stderr)
         sys.exit(3)
 
-    # latent warm-up: the library solves steps 1..T_w (alpha = 1) and then the rest, so an update
-    # of the first part covers T_w steps and one of the rest T - T_w.  The first part's update
-    # count is that of the same solve run on its own (deterministic), taken once, untimed.
+    # latent warm-up: inside the one Newton iteration every update covers all T steps; where the
+    # library solves steps 1..T_w (alpha = 1) and then the rest, an update of the first part
+    # covers T_w steps and one of the rest T - T_w.  The first part's update count is that of the
+    # same solve run on its own (deterministic), taken once, untimed.
     warm_updates = None
-    if args.tw and c.kind in ("plrnn", "shplrnn") and not args.quasi:
+    if (args.tw and c.kind in ("plrnn", "shplrnn") and not args.quasi
+            and not warmup_in_one_iteration(c.kind, c.M, args.quasi)):
         r1 = D.deer_solve(model, xd[:, :args.tw + 1].contiguous(), 1.0, c.n_obs, tol=c.tol, max_iter=c.max_iter,
                           check=False)
         warm_updates = int(sum(r1["iters"]))

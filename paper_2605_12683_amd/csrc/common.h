@@ -131,7 +131,7 @@ __device__ __forceinline__ void wave_lds_sync() {
 
 __device__ __forceinline__ float forced_state(const float *__restrict__ x, const float *__restrict__ z0,
                                               const float *__restrict__ z, int b, int s, int i, int T, int M,
-                                              int N, float alpha) {
+                                              int N, float alpha, int tw = 0) {
     if (s == 0) {
         if (z0) return z0[(size_t)b * M + i];
         return i < N ? x[(size_t)b * (T + 1) * N + i] : 0.0f;
@@ -139,6 +139,7 @@ __device__ __forceinline__ float forced_state(const float *__restrict__ x, const
     float zp = z[((size_t)b * T + (s - 1)) * M + i];
     if (i >= N) return zp;
     float zb = x[((size_t)b * (T + 1) + s) * N + i];
+    if (s <= tw) return zb;   // latent warm-up: alpha_s = 1 for s = 1..tw
     float p = __fsub_rn(1.0f, alpha);
     return __fadd_rn(__fmul_rn(p, zp), __fmul_rn(alpha, zb));
 }

@@ -862,6 +862,13 @@ static int init_guess(const deer_solve_opts *o, int B, int T, int M, int N, cons
     return DEER_OK;
 }
 
+// The latent warm-up inside the one Newton iteration (per-step forcing strength in the kernels):
+// the register-tiled vanilla PLRNN path (M <= 16) with the identity read-out.  The other paths
+// solve the warm-up prefix and the rest as two chained problems (solve_warmup below).
+static bool warmup_joint(const deer_model *m, const deer_forcing *f) {
+    return f->T_w > 0 && !f->obs && m->kind == DEER_PLRNN && m->M <= 16;
+}
+
 static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
                        const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
                        void *ws, size_t ws_bytes, hipStream_t st) {
@@ -871,11 +878,12 @@ static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_so
     if (rc) return rc;
     PlrnnWs w = carve_plrnn(ws, B, T, m->M, DEER_OP_SOLVE, &need);
     PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
+    a.tw = f->T_w;
     if ((rc = init_guess(o, B, T, m->M, f->n_forced, x, z, st))) return rc;
     std::vector<int> act(B, 1), it(B, 0);
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
-    if (small_path_enabled() && newton_small_fits(m->M, T, o->fixed_iters)) {
+    if (a.tw == 0 && small_path_enabled() && newton_small_fits(m->M, T, o->fixed_iters)) {
         // every update in one launch; the last update's norms read once
         if ((rc = launch_newton_small(a, z, o->fixed_iters, w.ctl.norm_bits, st))) return rc;
         std::vector<uint32_t> nb(B, 0);
@@ -1559,7 +1567,8 @@ int deer_solve(const deer_model *m, const deer_forcing *f, const deer_solve_opts
     if (m->kind != DEER_DIAG_SSM && o->fixed_iters <= 0 && (rc = check_host_reserved(B))) return rc;
     hipStream_t st = (hipStream_t)stream;
     if (f->obs) return solve_obs(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
-    if (f->T_w > 0) return solve_warmup(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st, false);
+    if (f->T_w > 0 && !warmup_joint(m, f))
+        return solve_warmup(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st, false);
     if (m->kind == DEER_PLRNN)
         return solve_plrnn(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
     if (m->kind == DEER_SHPLRNN)
@@ -1599,18 +1608,21 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
     if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
     hipStream_t st = (hipStream_t)stream;
     if (f->obs) return adjoint_obs(m, f, B, T, x, z0, z, g, lam, grads, ws, ws_bytes, st);
-    if (f->T_w > 0) {
-        if (g_layout != DEER_G_NATIVE) { set_error("the latent warm-up takes the native cotangent layout"); return DEER_ERR_INVALID_ARG; }
-        return adjoint_warmup(m, f, B, T, x, z0, z, g, lam, grads, ws, ws_bytes, st, false);
+    if (f->T_w > 0 && g_layout != DEER_G_NATIVE) {
+        set_error("the latent warm-up takes the native cotangent layout");
+        return DEER_ERR_INVALID_ARG;
     }
+    if (f->T_w > 0 && !warmup_joint(m, f)) return adjoint_warmup(m, f, B, T, x, z0, z, g, lam, grads, ws, ws_bytes, st, false);
     if (m->kind == DEER_PLRNN) {
         size_t need = 0;
         carve_plrnn(nullptr, B, T, m->M, DEER_OP_ADJOINT, &need);
         if ((rc = check_ws(ws, ws_bytes, need))) return rc;
         PlrnnWs w = carve_plrnn(ws, B, T, m->M, DEER_OP_ADJOINT, &need);
         PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
-        const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
-        if (small_path_enabled() && adjoint_small_fits(m->M, T)) {   // one workgroup per sequence
+        a.tw = f->T_w;   // > 0 only on the register-tiled path (M <= 16)
+        // MSE seed over the states after the warm-up, z_{T_w+1}..z_T
+        const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * (T - f->T_w))) : 0.f;
+        if (a.tw == 0 && small_path_enabled() && adjoint_small_fits(m->M, T)) {   // one workgroup per sequence
             const bool gr = grads && (grads->A || grads->W || grads->h);
             if (B == 1)
                 return launch_adjoint_small(a, g, scale, z, lam, nullptr, gr ? grads->A : nullptr,
@@ -1750,6 +1762,8 @@ size_t deer_workspace_bytes_ex(const deer_model *m, const deer_forcing *f, int B
     }
     if (!f || f->T_w == 0) return quasi ? deer_quasi_workspace_bytes(m, B, T, op) : deer_workspace_bytes(m, B, T, op);
     if ((quasi ? check_quasi(m, f, B, T) : check_common(m, f, B, T)) != DEER_OK) return 0;
+    if (!quasi && warmup_joint(m, f) && (op == DEER_OP_SOLVE || op == DEER_OP_ADJOINT))
+        return deer_workspace_bytes(m, B, T, op);   // one iteration over the whole sequence
     if (op != DEER_OP_SOLVE && op != DEER_OP_ADJOINT) return 0;
     size_t bytes = 0;
     carve_warm(nullptr, m, f, B, T, op, quasi != 0, &bytes);

@@ -29,6 +29,18 @@ struct Geo {
 
 __device__ __forceinline__ float p_of(int i, int N, float alpha) { return i < N ? __fsub_rn(1.0f, alpha) : 1.0f; }
 
+// Latent warm-up (section "Latent state warm-up", Alg. GTF-DEER): the forced inputs of steps
+// s = 1..tw replace the observed latents by the data (alpha_s = 1, P_1), so those steps'
+// Jacobians have the observed columns zeroed.  Kernels take it as a template flag WU; without it
+// the warm-up code compiles away.  Step 0's Jacobian multiplies the fixed initial state's zero
+// update, so it may count as a warm-up step too.
+template <bool WU>
+__device__ __forceinline__ float forced_in(float pi, float alpha, float zp, float xs, int s, int tw) {
+    const float f = __fadd_rn(__fmul_rn(pi, zp), __fmul_rn(alpha, xs));
+    if constexpr (WU) return s <= tw ? xs : f;
+    return f;
+}
+
 __device__ __forceinline__ uint32_t mask_bit(const uint32_t *__restrict__ masks, size_t step, int MW, int i) {
     return (masks[step * MW + (i >> 5)] >> (i & 31)) & 1u;
 }
@@ -663,6 +675,7 @@ __device__ __forceinline__ float rfl_f(float v) { return __int_as_float(__builti
 // of the four chains are loaded at once (clamped indices) and combined afterwards.
 struct Chains16 {
     int plen[4];
+    int cs[4];   // first step of each chain in its sequence
     float gam[4];
     int minlen, maxlen;
     bool onebuf;
@@ -697,6 +710,7 @@ __device__ __forceinline__ Chains16 chains16(int chain0, int nchains, int ncs, i
     for (int n = 0; n < 4; ++n) {
         const bool ok = chain0 + n < nchains && act[n] != 0;
         w.plen[n] = ok ? min(C, T - cq[n] * C) : 0;
+        w.cs[n] = cq[n] * C;
         if (w.plen[n] > 0) {
             if (sel0 >= 0 && sel[n] != sel0) w.onebuf = false;
             sel0 = sel[n];
@@ -753,16 +767,42 @@ __device__ __forceinline__ v4f mfma_step16(const v4f &acc, uint32_t wn, int g, c
     return nx;
 }
 
+// bits tt < n of a tile's step mask (n may lie outside 0..32)
+__device__ __forceinline__ uint32_t low_bits(int n) { return n <= 0 ? 0u : (n >= 32 ? ~0u : (1u << n) - 1u); }
+
+// forced input of an observed latent at tile row tt; in a tile holding warm-up steps, bit tt of
+// wb marks one (the data itself, alpha_s = 1)
+template <bool WT>
+__device__ __forceinline__ float forced_at(float pi, float alpha, float zp, float xs, uint32_t wb, int tt) {
+    const float f = __fadd_rn(__fmul_rn(pi, zp), __fmul_rn(alpha, xs));
+    if constexpr (WT) return ((wb >> tt) & 1u) ? xs : f;
+    return f;
+}
+
+// mfma_step16 in a warm-up step: the product's rows of the observed latents (fr[q]: row
+// 4 g + q) are left out of the B operand, which is J~ = J_F P_1 acting on it
+__device__ __forceinline__ v4f mfma_step16_warm(const v4f &acc, uint32_t wn, int g, const float (&WpD)[4],
+                                                const float (&Dq)[4], const bool (&fr)[4]) {
+    v4f nx = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)wn, 4 * g + q, 1);
+        const float a = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+        nx = mfma16x16x4(a, fr[q] ? 0.f : acc[q], nx);
+    }
+    return nx;
+}
+
 // WPB waves per block (1, or 8 for the group maps: the block's 32 chunks then belong to one
 // sequence); wmaps: 0 plain chunk aggregates, 1 wave maps, 2 wave maps composed per block into
 // group maps (gmap).
-template <int TB, int WPB>
+template <int TB, int WPB, bool WU>
 __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
     const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
     const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
     const int *__restrict__ zsel, float *__restrict__ Pout,
     float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
-    int ncs, int wmaps, float *__restrict__ gmap, uint32_t *mark, uint32_t pass_no) {
+    int ncs, int wmaps, float *__restrict__ gmap, uint32_t *mark, uint32_t pass_no, int tw) {
     // the wave index is uniform: the chain set, its control words and the tile addresses are
     // scalar values (scalar loads, no per-lane address arithmetic)
     const int lane = threadIdx.x & 63, wvb = WPB > 1 ? rfl_i((int)(threadIdx.x >> 6)) : 0, g = lane >> 4, c = lane & 15;
@@ -786,6 +826,9 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
             ugam = w.gam[n];
         }
     const bool lat = c < M, forced = c < N;
+    bool fr[4];   // B-operand rows 4 g + q of observed latents (dropped in warm-up steps)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) fr[q] = 4 * g + q < N;
     // tile resources, based at the first row of the wave's first chain
     const int b0 = chain0 / ncs, s00 = (chain0 % ncs) * C;
     const size_t row0 = (size_t)b0 * T + s00, xrow0 = (size_t)b0 * (T + 1) + s00;
@@ -841,48 +884,107 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
                     xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
                 }
             }
-            // residual and masks of every step of the tile, two steps at a time; r overwrites zv
-            uint32_t posb = 0u;
+            bool wtile = false;   // some chain of the wave has a latent warm-up step in this tile
+            if constexpr (WU) {
 #pragma unroll
-            for (int tt = 0; tt < TB; tt += 2) {
-                const int s = s0 + t0 + tt;
-                const float zt0 =
-                    (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xv[tt]));
-                const float zt1 = !forced ? zv[tt] : __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt + 1]));
-                const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
-                posb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
-                float d0, d1;
-                row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
-                const float F0 = fmaf(Ai, zt0, d0) + hi, F1 = fmaf(Ai, zt1, d1) + hi;
-                zprev = zv[tt + 1];
-                zv[tt] = zv[tt] - F0;
-                zv[tt + 1] = zv[tt + 1] - F1;
+                for (int n = 0; n < 4; ++n) wtile = wtile || w.cs[n] + t0 <= tw;
             }
-            // serial part: chunk products and chunk-local solutions
+            if (wtile) {
+                // the tile body below with the warm-up steps' P_1: the observed latents' rows of
+                // the B operand and of u dropped, their forced inputs the data
+                const uint32_t wb = low_bits(tw - (s0 + t0) + 1);   // bit tt: s0 + t0 + tt <= tw
+                int lim[4];   // chain n: tile steps tt < lim[n] are warm-up steps
 #pragma unroll
-            for (int tt = 0; tt < TB; ++tt) {
-                const bool pos = (posb >> tt) & 1u;
-                const uint64_t bal = __ballot(pos);
-                // the four chains' updates interleaved: k-slice outer, chain inner
-                float Am[4][4];
+                for (int n = 0; n < 4; ++n) lim[n] = tw - (w.cs[n] + t0) + 1;
+                uint32_t posb = 0u;
 #pragma unroll
-                for (int n = 0; n < 4; ++n)
+                for (int tt = 0; tt < TB; tt += 2) {
+                    const int s = s0 + t0 + tt;
+                    const float zt0 = (s == 0 || !forced) ? zprev : forced_at<true>(pi, alpha, zprev, xv[tt], wb, tt);
+                    const float zt1 = !forced ? zv[tt] : forced_at<true>(pi, alpha, zv[tt], xv[tt + 1], wb, tt + 1);
+                    const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
+                    posb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
+                    float d0, d1;
+                    row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
+                    const float F0 = fmaf(Ai, zt0, d0) + hi, F1 = fmaf(Ai, zt1, d1) + hi;
+                    zprev = zv[tt + 1];
+                    zv[tt] = zv[tt] - F0;
+                    zv[tt + 1] = zv[tt + 1] - F1;
+                }
+                const uint32_t wf = forced ? wb : 0u;
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
-                        Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
-                    }
-                v4f nx[4];
+                for (int tt = 0; tt < TB; ++tt) {
+                    const bool pos = (posb >> tt) & 1u;
+                    const uint64_t bal = __ballot(pos);
+                    float Am[4][4];
 #pragma unroll
-                for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
+                    for (int n = 0; n < 4; ++n)
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t m =
+                                (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
+                            Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+                        }
+                    v4f nx[4];
 #pragma unroll
-                    for (int n = 0; n < 4; ++n) nx[n] = mfma16x16x4(Am[n][q], acc[n][q], nx[n]);
+                    for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int n = 0; n < 4; ++n) acc[n] = nx[n];
-                const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
-                u = fmaf(ugam, y, -zv[tt]);
+                    for (int q = 0; q < 4; ++q)
+#pragma unroll
+                        for (int n = 0; n < 4; ++n)
+                            nx[n] = mfma16x16x4(Am[n][q], (fr[q] && tt < lim[n]) ? 0.f : acc[n][q], nx[n]);
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) acc[n] = nx[n];
+                    const float uo = ((wf >> tt) & 1u) ? 0.f : u;
+                    const float y = fmaf(di, uo, row16_dot(wr, pos ? pi * uo : 0.f));
+                    u = fmaf(ugam, y, -zv[tt]);
+                }
+            } else {
+                // residual and masks of every step of the tile, two steps at a time; r overwrites zv
+                uint32_t posb = 0u;
+#pragma unroll
+                for (int tt = 0; tt < TB; tt += 2) {
+                    const int s = s0 + t0 + tt;
+                    const float zt0 =
+                        (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xv[tt]));
+                    const float zt1 =
+                        !forced ? zv[tt] : __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt + 1]));
+                    const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
+                    posb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
+                    float d0, d1;
+                    row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
+                    const float F0 = fmaf(Ai, zt0, d0) + hi, F1 = fmaf(Ai, zt1, d1) + hi;
+                    zprev = zv[tt + 1];
+                    zv[tt] = zv[tt] - F0;
+                    zv[tt + 1] = zv[tt + 1] - F1;
+                }
+                // serial part: chunk products and chunk-local solutions
+#pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    const bool pos = (posb >> tt) & 1u;
+                    const uint64_t bal = __ballot(pos);
+                    // the four chains' updates interleaved: k-slice outer, chain inner
+                    float Am[4][4];
+#pragma unroll
+                    for (int n = 0; n < 4; ++n)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t m =
+                                (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
+                            Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+                        }
+                    v4f nx[4];
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+#pragma unroll
+                        for (int n = 0; n < 4; ++n) nx[n] = mfma16x16x4(Am[n][q], acc[n][q], nx[n]);
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) acc[n] = nx[n];
+                    const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
+                    u = fmaf(ugam, y, -zv[tt]);
+                }
             }
         } else {
             for (int t = t0; t < t0 + tl; ++t) {
@@ -894,15 +996,22 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
                     if (forced && s > 0) xb = x[((size_t)b * (T + 1) + s) * N + c];
                 }
                 float zt = 0.f;
-                if (run) zt = (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xb));
+                if (run) zt = (s == 0 || !forced) ? zprev : forced_in<WU>(pi, alpha, zprev, xb, s, tw);
                 const bool pos = zt > 0.f;
                 const uint64_t bal = __ballot(pos);
                 const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
                 const float r = zcur - F;
 #pragma unroll
                 for (int n = 0; n < 4; ++n)
-                    if (t < w.plen[n]) acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
-                const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
+                    if (t < w.plen[n]) {
+                        if (WU && w.cs[n] + t <= tw)
+                            acc[n] = mfma_step16_warm(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq, fr);
+                        else
+                            acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
+                    }
+                float uo = u;
+                if constexpr (WU) uo = (forced && s <= tw) ? 0.f : u;
+                const float y = fmaf(di, uo, row16_dot(wr, pos ? pi * uo : 0.f));
                 if (run) {
                     u = fmaf(ugam, y, -r);
                     zprev = zcur;
@@ -1086,7 +1195,7 @@ __device__ __forceinline__ void seq_arrive(const FusedCtl &fc, int b, int cnt, i
 // and reading them here; Delta_t = gamma (diag(d) + W p diag(m_t)) Delta_{t-1} - r_t from the
 // chunk's carry, z + Delta written to the other iterate buffer, per-chain max |Delta| and max
 // |z|, and (with fc.seq) the pass-end control of the sequence.
-template <int TB>
+template <int TB, bool WU>
 __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restrict__ A, const float *__restrict__ W,
                                                           const float *__restrict__ h, float alpha, int N,
                                                           const float *__restrict__ x, const float *__restrict__ z0,
@@ -1097,7 +1206,7 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
                                                           const float *__restrict__ gamma, int B, int T, int M, int C,
                                                           int ncs, const float *__restrict__ Pm,
                                                           const float *__restrict__ vmap,
-                                                          const float *__restrict__ gmap, FusedCtl fc) {
+                                                          const float *__restrict__ gmap, FusedCtl fc, int tw) {
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int nchains = B * ncs;
     const int chain0 = blockIdx.x * 4;
@@ -1221,29 +1330,63 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
                 zv[tt] = bload(rzi, vz, 4 * (t0 + tt) * M);
                 rv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);   // x of the step, replaced by r below
             }
-            // residual and masks of the tile (as in the forward pass)
-            uint32_t mb = 0u;
+            // a tile holding latent warm-up steps of this lane's chunk runs the body with P_1 there
+            bool wtile = false;
+            if constexpr (WU) {
 #pragma unroll
-            for (int tt = 0; tt < TB; ++tt) {
-                const int s = s0 + t0 + tt;
-                const float zt =
-                    (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, rv[tt]));
-                const bool pos = zt > 0.f;
-                mb |= (pos ? 1u : 0u) << tt;
-                const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
-                zprev = zv[tt];
-                rv[tt] = zv[tt] - F;
+                for (int n = 0; n < 4; ++n) wtile = wtile || w.cs[n] + t0 <= tw;
             }
-#pragma unroll
-            for (int tt = 0; tt < TB; ++tt) {
-                const bool m = (mb >> tt) & 1u;
-                const float y = fmaf(d, D, row16_dot(wp, m ? D : 0.f));
-                D = fmaf(gm, y, -rv[tt]);
-                const float zc = zv[tt];
-                bstore_u(rzo, __float_as_uint(zc + D), vz, 4 * (t0 + tt) * M);
-                const uint32_t ab = abs_bits(D), zb = abs_bits(zc);
-                emax = emax > ab ? emax : ab;
-                zmax = zmax > zb ? zmax : zb;
+            if (wtile) {
+                const uint32_t wb = low_bits(tw - (s0 + t0) + 1);   // bit tt: s0 + t0 + tt <= tw
+                const uint32_t wf = forced ? wb : 0u;
+                // residual and masks of the tile (as in the forward pass)
+                uint32_t mb = 0u;
+    #pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    const int s = s0 + t0 + tt;
+                    const float zt = (s == 0 || !forced) ? zprev : forced_at<true>(pi, alpha, zprev, rv[tt], wb, tt);
+                    const bool pos = zt > 0.f;
+                    mb |= (pos ? 1u : 0u) << tt;
+                    const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
+                    zprev = zv[tt];
+                    rv[tt] = zv[tt] - F;
+                }
+    #pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    const bool m = (mb >> tt) & 1u;
+                    const float Do = ((wf >> tt) & 1u) ? 0.f : D;   // P_1: observed entries dropped
+                    const float y = fmaf(d, Do, row16_dot(wp, m ? Do : 0.f));
+                    D = fmaf(gm, y, -rv[tt]);
+                    const float zc = zv[tt];
+                    bstore_u(rzo, __float_as_uint(zc + D), vz, 4 * (t0 + tt) * M);
+                    const uint32_t ab = abs_bits(D), zb = abs_bits(zc);
+                    emax = emax > ab ? emax : ab;
+                    zmax = zmax > zb ? zmax : zb;
+                }
+            } else {
+                // residual and masks of the tile (as in the forward pass)
+                uint32_t mb = 0u;
+    #pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    const int s = s0 + t0 + tt;
+                    const float zt = (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, rv[tt]));
+                    const bool pos = zt > 0.f;
+                    mb |= (pos ? 1u : 0u) << tt;
+                    const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
+                    zprev = zv[tt];
+                    rv[tt] = zv[tt] - F;
+                }
+    #pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    const bool m = (mb >> tt) & 1u;
+                    const float y = fmaf(d, D, row16_dot(wp, m ? D : 0.f));
+                    D = fmaf(gm, y, -rv[tt]);
+                    const float zc = zv[tt];
+                    bstore_u(rzo, __float_as_uint(zc + D), vz, 4 * (t0 + tt) * M);
+                    const uint32_t ab = abs_bits(D), zb = abs_bits(zc);
+                    emax = emax > ab ? emax : ab;
+                    zmax = zmax > zb ? zmax : zb;
+                }
             }
         } else {
             for (int t = t0; t < t0 + tl; ++t) {
@@ -1256,11 +1399,13 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
                     if (forced && s > 0) xb = x[((size_t)b * (T + 1) + s) * N + c];
                 }
                 float zt = 0.f;
-                if (run) zt = (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xb));
+                if (run) zt = (s == 0 || !forced) ? zprev : forced_in<WU>(pi, alpha, zprev, xb, s, tw);
                 const bool pos = zt > 0.f;
                 const float F = fmaf(Ai, zt, row16_dot(wr, pos ? zt : 0.f)) + hi;
                 const float rc = zc - F;
-                const float y = fmaf(d, D, row16_dot(wp, (run && pos) ? D : 0.f));
+                float Do = D;
+                if constexpr (WU) Do = (forced && s <= tw) ? 0.f : D;
+                const float y = fmaf(d, Do, row16_dot(wp, (run && pos) ? Do : 0.f));
                 if (run) {
                     D = fmaf(gm, y, -rc);
                     zout[step * M + c] = zc + D;
@@ -1332,13 +1477,13 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn16(const float *__restric
 // wave's carry with the same operations on the same operands instead of taking the end of its
 // own recurrence, the same Delta to rounding), so no wave waits for another.
 // ---------------------------------------------------------------------------------------
-template <int TB>
+template <int TB, bool WU>
 __global__ __launch_bounds__(512) void k_newton_pass16(
     const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
     const float *__restrict__ x, const float *__restrict__ z0, float *zbuf, float *zalt, int T, int M, int C, int ncs,
     const float *__restrict__ Pin, const float *__restrict__ vin, const float *__restrict__ gin,
     float *__restrict__ Pout, float *__restrict__ vout, float *__restrict__ gout, FusedCtl fc, uint32_t *mark,
-    uint32_t pass_no) {
+    uint32_t pass_no, int tw) {
     constexpr int WPB = 8;
     const int lane = threadIdx.x & 63, wvb = rfl_i((int)(threadIdx.x >> 6)), g = lane >> 4, c = lane & 15;
     if (mark && blockIdx.x == 0 && threadIdx.x == 0)
@@ -1358,6 +1503,9 @@ __global__ __launch_bounds__(512) void k_newton_pass16(
     float *const zn = sel ? zbuf : zalt;   // the update's output
     const int s0 = (cc0 + g) * C;          // first step of this lane's chunk
     const bool lat = c < M, forced = c < N;
+    bool fr[4];   // B-operand rows 4 g + q of observed latents (dropped in warm-up steps)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) fr[q] = 4 * g + q < N;
     const size_t row0 = (size_t)b * T + (size_t)cc0 * C, xrow0 = (size_t)b * (T + 1) + (size_t)cc0 * C;
     const auto rzc = wave_rsrc(zc + row0 * M), rzn = wave_rsrc(zn + row0 * M);
     const auto rx = wave_rsrc(N > 0 ? x + xrow0 * N : zc);
@@ -1516,36 +1664,74 @@ __global__ __launch_bounds__(512) void k_newton_pass16(
                     xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
                 }
             }
-            float rv[TB];
-            uint32_t mb = 0u;
-#pragma unroll
-            for (int tt = 0; tt < TB; tt += 2) {
-                const int s = s0 + t0 + tt;
-                const float zt0 =
-                    (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xv[tt]));
-                const float zt1 = !forced ? zv[tt] : __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt + 1]));
-                const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
-                mb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
-                float d0, d1;
-                row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
-                rv[tt] = zv[tt] - (fmaf(Ai, zt0, d0) + hi);
-                rv[tt + 1] = zv[tt + 1] - (fmaf(Ai, zt1, d1) + hi);
-                zprev = zv[tt + 1];
-            }
-#pragma unroll
-            for (int tt = 0; tt < TB; ++tt) {
-                const bool m = (mb >> tt) & 1u;
-                const float y = fmaf(di, D, row16_dot(wp, m ? D : 0.f));
-                D = fmaf(gam, y, -rv[tt]);
-                const float zcur = zv[tt];
-                // the last step before the next wave: its Delta as that wave's carry
-                const float dap = (tt == TB - 1 && t0 + TB == C && nextc) ? Dnext : D;
-                const float znew = zcur + dap;
-                if (t0 + TB < C) bstore_u(rzn, __float_as_uint(znew), vz, 4 * (t0 + tt) * M);
-                const uint32_t ab = lat ? abs_bits(dap) : 0u, zb = abs_bits(zcur);
-                emax = emax > ab ? emax : ab;
-                zmax = zmax > zb ? zmax : zb;
-                zv[tt] = znew;
+            // a tile holding latent warm-up steps runs the body with P_1 in those steps
+            bool wtile = false;
+            if constexpr (WU) wtile = cc0 * C + t0 <= tw;
+            if (wtile) {
+                const uint32_t wb = low_bits(tw - (s0 + t0) + 1);   // bit tt: s0 + t0 + tt <= tw
+                const uint32_t wf = forced ? wb : 0u;
+                float rv[TB];
+                uint32_t mb = 0u;
+    #pragma unroll
+                for (int tt = 0; tt < TB; tt += 2) {
+                    const int s = s0 + t0 + tt;
+                    const float zt0 = (s == 0 || !forced) ? zprev : forced_at<true>(pi, alpha, zprev, xv[tt], wb, tt);
+                    const float zt1 = !forced ? zv[tt] : forced_at<true>(pi, alpha, zv[tt], xv[tt + 1], wb, tt + 1);
+                    const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
+                    mb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
+                    float d0, d1;
+                    row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
+                    rv[tt] = zv[tt] - (fmaf(Ai, zt0, d0) + hi);
+                    rv[tt + 1] = zv[tt + 1] - (fmaf(Ai, zt1, d1) + hi);
+                    zprev = zv[tt + 1];
+                }
+    #pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    const bool m = (mb >> tt) & 1u;
+                    const float Do = ((wf >> tt) & 1u) ? 0.f : D;   // P_1: observed entries dropped
+                    const float y = fmaf(di, Do, row16_dot(wp, m ? Do : 0.f));
+                    D = fmaf(gam, y, -rv[tt]);
+                    const float zcur = zv[tt];
+                    // the last step before the next wave: its Delta as that wave's carry
+                    const float dap = (tt == TB - 1 && t0 + TB == C && nextc) ? Dnext : D;
+                    const float znew = zcur + dap;
+                    if (t0 + TB < C) bstore_u(rzn, __float_as_uint(znew), vz, 4 * (t0 + tt) * M);
+                    const uint32_t ab = lat ? abs_bits(dap) : 0u, zb = abs_bits(zcur);
+                    emax = emax > ab ? emax : ab;
+                    zmax = zmax > zb ? zmax : zb;
+                    zv[tt] = znew;
+                }
+            } else {
+                float rv[TB];
+                uint32_t mb = 0u;
+    #pragma unroll
+                for (int tt = 0; tt < TB; tt += 2) {
+                    const int s = s0 + t0 + tt;
+                    const float zt0 = (s == 0 || !forced) ? zprev : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xv[tt]));
+                    const float zt1 = !forced ? zv[tt] : __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt + 1]));
+                    const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
+                    mb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
+                    float d0, d1;
+                    row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
+                    rv[tt] = zv[tt] - (fmaf(Ai, zt0, d0) + hi);
+                    rv[tt + 1] = zv[tt + 1] - (fmaf(Ai, zt1, d1) + hi);
+                    zprev = zv[tt + 1];
+                }
+    #pragma unroll
+                for (int tt = 0; tt < TB; ++tt) {
+                    const bool m = (mb >> tt) & 1u;
+                    const float y = fmaf(di, D, row16_dot(wp, m ? D : 0.f));
+                    D = fmaf(gam, y, -rv[tt]);
+                    const float zcur = zv[tt];
+                    // the last step before the next wave: its Delta as that wave's carry
+                    const float dap = (tt == TB - 1 && t0 + TB == C && nextc) ? Dnext : D;
+                    const float znew = zcur + dap;
+                    if (t0 + TB < C) bstore_u(rzn, __float_as_uint(znew), vz, 4 * (t0 + tt) * M);
+                    const uint32_t ab = lat ? abs_bits(dap) : 0u, zb = abs_bits(zcur);
+                    emax = emax > ab ? emax : ab;
+                    zmax = zmax > zb ? zmax : zb;
+                    zv[tt] = znew;
+                }
             }
         }
         // z_{s0-1} of the new iterate exactly as stored: chunks 1..3 of the wave take it from the
@@ -1576,45 +1762,97 @@ __global__ __launch_bounds__(512) void k_newton_pass16(
                 xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
             }
         }
-        // residual and masks; r overwrites zv
-        uint32_t posb = 0u;
+        bool wtile = false;   // a tile holding latent warm-up steps: P_1 in those steps
+        if constexpr (WU) wtile = cc0 * C + t0 <= tw;
+        if (wtile) {
+            const uint32_t wb = low_bits(tw - (s0 + t0) + 1);   // bit tt: s0 + t0 + tt <= tw
+            const uint32_t wf = forced ? wb : 0u;
+            int lim[4];   // chain n: tile steps tt < lim[n] are warm-up steps
 #pragma unroll
-        for (int tt = 0; tt < TB; tt += 2) {
-            const int s = s0 + t0 + tt;
-            const float zt0 = (s == 0 || !forced) ? zpn : __fadd_rn(__fmul_rn(pi, zpn), __fmul_rn(alpha, xv[tt]));
-            const float zt1 = !forced ? zv[tt] : __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt + 1]));
-            const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
-            posb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
-            float d0, d1;
-            row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
-            const float F0 = fmaf(Ai, zt0, d0) + hi, F1 = fmaf(Ai, zt1, d1) + hi;
-            zpn = zv[tt + 1];
-            zv[tt] = zv[tt] - F0;
-            zv[tt + 1] = zv[tt + 1] - F1;
-        }
-#pragma unroll
-        for (int tt = 0; tt < TB; ++tt) {
-            const bool pos = (posb >> tt) & 1u;
-            const uint64_t bal = __ballot(pos);
-            float Am[4][4];
-#pragma unroll
-            for (int n = 0; n < 4; ++n)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
-                    Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
-                }
-            v4f nx[4];
-#pragma unroll
-            for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int n = 0; n < 4; ++n) nx[n] = mfma16x16x4(Am[n][q], acc[n][q], nx[n]);
-#pragma unroll
-            for (int n = 0; n < 4; ++n) acc[n] = nx[n];
-            const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
-            u = fmaf(gnext, y, -zv[tt]);
+            for (int n = 0; n < 4; ++n) lim[n] = tw - ((cc0 + n) * C + t0) + 1;
+            // residual and masks; r overwrites zv
+            uint32_t posb = 0u;
+    #pragma unroll
+            for (int tt = 0; tt < TB; tt += 2) {
+                const int s = s0 + t0 + tt;
+                const float zt0 = (s == 0 || !forced) ? zpn : forced_at<true>(pi, alpha, zpn, xv[tt], wb, tt);
+                const float zt1 = !forced ? zv[tt] : forced_at<true>(pi, alpha, zv[tt], xv[tt + 1], wb, tt + 1);
+                const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
+                posb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
+                float d0, d1;
+                row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
+                const float F0 = fmaf(Ai, zt0, d0) + hi, F1 = fmaf(Ai, zt1, d1) + hi;
+                zpn = zv[tt + 1];
+                zv[tt] = zv[tt] - F0;
+                zv[tt + 1] = zv[tt + 1] - F1;
+            }
+    #pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                const bool pos = (posb >> tt) & 1u;
+                const uint64_t bal = __ballot(pos);
+                float Am[4][4];
+    #pragma unroll
+                for (int n = 0; n < 4; ++n)
+    #pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
+                        Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+                    }
+                v4f nx[4];
+    #pragma unroll
+                for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+                for (int q = 0; q < 4; ++q)
+    #pragma unroll
+                    for (int n = 0; n < 4; ++n)
+                        nx[n] = mfma16x16x4(Am[n][q], (fr[q] && tt < lim[n]) ? 0.f : acc[n][q], nx[n]);
+    #pragma unroll
+                for (int n = 0; n < 4; ++n) acc[n] = nx[n];
+                const float uo = ((wf >> tt) & 1u) ? 0.f : u;
+                const float y = fmaf(di, uo, row16_dot(wr, pos ? pi * uo : 0.f));
+                u = fmaf(gnext, y, -zv[tt]);
+            }
+        } else {
+            // residual and masks; r overwrites zv
+            uint32_t posb = 0u;
+    #pragma unroll
+            for (int tt = 0; tt < TB; tt += 2) {
+                const int s = s0 + t0 + tt;
+                const float zt0 = (s == 0 || !forced) ? zpn : __fadd_rn(__fmul_rn(pi, zpn), __fmul_rn(alpha, xv[tt]));
+                const float zt1 = !forced ? zv[tt] : __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt + 1]));
+                const bool p0 = zt0 > 0.f, p1 = zt1 > 0.f;
+                posb |= ((p0 ? 1u : 0u) | (p1 ? 2u : 0u)) << tt;
+                float d0, d1;
+                row16_dot2(wr, p0 ? zt0 : 0.f, p1 ? zt1 : 0.f, d0, d1);
+                const float F0 = fmaf(Ai, zt0, d0) + hi, F1 = fmaf(Ai, zt1, d1) + hi;
+                zpn = zv[tt + 1];
+                zv[tt] = zv[tt] - F0;
+                zv[tt + 1] = zv[tt + 1] - F1;
+            }
+    #pragma unroll
+            for (int tt = 0; tt < TB; ++tt) {
+                const bool pos = (posb >> tt) & 1u;
+                const uint64_t bal = __ballot(pos);
+                float Am[4][4];
+    #pragma unroll
+                for (int n = 0; n < 4; ++n)
+    #pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
+                        Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+                    }
+                v4f nx[4];
+    #pragma unroll
+                for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+                for (int q = 0; q < 4; ++q)
+    #pragma unroll
+                    for (int n = 0; n < 4; ++n) nx[n] = mfma16x16x4(Am[n][q], acc[n][q], nx[n]);
+    #pragma unroll
+                for (int n = 0; n < 4; ++n) acc[n] = nx[n];
+                const float y = fmaf(di, u, row16_dot(wr, pos ? pi * u : 0.f));
+                u = fmaf(gnext, y, -zv[tt]);
+            }
         }
         if (gnext != 1.f) {
 #pragma unroll
@@ -2188,11 +2426,12 @@ __device__ __forceinline__ void row16_outer(float (&d)[16], float v, float s) {
 // t0 + tt: z_{s0+t0+tt}, x_{s0+t0+tt+1} (so z~ of step s0+t0+tt+1, the mask lam_k needs) and
 // g_{s0+t0+tt}.  The products run forward over the tiles, the local adjoint backward.
 // ---------------------------------------------------------------------------------------
-template <int TB>
+template <int TB, bool WU>
 __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
     const float *__restrict__ A, const float *__restrict__ W, float alpha, int N, const float *__restrict__ rhs,
     const float *__restrict__ z, const float *__restrict__ x, float seed_scale, float *__restrict__ Pout,
-    float *__restrict__ vout, int B, int T, int M, int C, int ncs, int wmaps) {
+    float *__restrict__ vout, int B, int T, int M, int C, int ncs, int wmaps, int tw) {
+    static_assert(!WU || TB <= 16, "the warm-up variant runs 16-step tiles");
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int nchains = B * ncs;
     const int chain0 = blockIdx.x * 4;
@@ -2228,6 +2467,9 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
     for (int n = 0; n < 4; ++n)
         if (n == g) len = w.plen[n];
     const bool lat = c < M, forced = c < N;
+    bool fr[4];   // B-operand rows 4 g + q of observed latents (dropped in warm-up steps)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) fr[q] = 4 * g + q < N;
     int src[16];
     row_sources(c, src);
     float wT[16];   // rotated row c of W^T
@@ -2253,9 +2495,11 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
             xv[tt] = bload(rx, vx, 4 * (t0 + tt) * N);
         }
         posb = 0u;
+        uint32_t wb = 0u;   // bit tt: step s0 + t0 + tt + 1 is a latent warm-up step
+        if constexpr (WU) wb = low_bits(tw - (s0 + t0));
 #pragma unroll
         for (int tt = 0; tt < TB; ++tt) {
-            const float zt = forced ? __fadd_rn(__fmul_rn(pi, zv[tt]), __fmul_rn(alpha, xv[tt])) : zv[tt];
+            const float zt = forced ? forced_at<WU>(pi, alpha, zv[tt], xv[tt], wb, tt) : zv[tt];
             posb |= (zt > 0.f ? 1u : 0u) << tt;
         }
         loaded = t0;
@@ -2266,7 +2510,7 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
         const int s = s0 + t + 1;
         const float zp = z[((size_t)b * T + s - 1) * M + c];
         if (!forced) return zp;
-        return __fadd_rn(__fmul_rn(pi, zp), __fmul_rn(alpha, x[((size_t)b * (T + 1) + s) * N + c]));
+        return forced_in<WU>(pi, alpha, zp, x[((size_t)b * (T + 1) + s) * N + c], s, tw);
     };
     // ---- chunk products, forward over the tiles
     for (int t0 = 0; t0 < w.maxlen; t0 += TB) {
@@ -2274,27 +2518,61 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
         if (t0 + TB <= w.minlen) {
             load_tile(t0);
             if (t0 + TB <= minP) {
+                bool wtile = false;   // some chain has a latent warm-up step in this tile
+                if constexpr (WU) {
 #pragma unroll
-                for (int tt = 0; tt < TB; ++tt) {
-                    const uint64_t bal = __ballot((posb >> tt) & 1u);
-                    float Am[4][4];
+                    for (int n = 0; n < 4; ++n) wtile = wtile || w.cs[n] + t0 + 1 <= tw;
+                }
+                if (wtile) {
+                    int lim[4];   // chain n: the steps of tile rows tt < lim[n] are warm-up steps
 #pragma unroll
-                    for (int n = 0; n < 4; ++n)
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const uint32_t m =
-                                (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
-                            Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
-                        }
-                    v4f nx[4];
-#pragma unroll
-                    for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-#pragma unroll
-                        for (int n = 0; n < 4; ++n) nx[n] = mfma16x16x4(Am[n][q], acc[n][q], nx[n]);
-#pragma unroll
-                    for (int n = 0; n < 4; ++n) acc[n] = nx[n];
+                    for (int n = 0; n < 4; ++n) lim[n] = tw - (w.cs[n] + t0);
+    #pragma unroll
+                    for (int tt = 0; tt < TB; ++tt) {
+                        const uint64_t bal = __ballot((posb >> tt) & 1u);
+                        float Am[4][4];
+    #pragma unroll
+                        for (int n = 0; n < 4; ++n)
+    #pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                const uint32_t m =
+                                    (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
+                                Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+                            }
+                        v4f nx[4];
+    #pragma unroll
+                        for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+                        for (int q = 0; q < 4; ++q)
+    #pragma unroll
+                            for (int n = 0; n < 4; ++n)
+                                nx[n] = mfma16x16x4(Am[n][q], (fr[q] && tt < lim[n]) ? 0.f : acc[n][q], nx[n]);
+    #pragma unroll
+                        for (int n = 0; n < 4; ++n) acc[n] = nx[n];
+                    }
+                } else {
+    #pragma unroll
+                    for (int tt = 0; tt < TB; ++tt) {
+                        const uint64_t bal = __ballot((posb >> tt) & 1u);
+                        float Am[4][4];
+    #pragma unroll
+                        for (int n = 0; n < 4; ++n)
+    #pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                const uint32_t m =
+                                    (uint32_t)__builtin_amdgcn_sbfe((int)(uint32_t)(bal >> (16 * n)), 4 * g + q, 1);
+                                Am[n][q] = __uint_as_float((m & __float_as_uint(WpD[q])) | (~m & __float_as_uint(Dq[q])));
+                            }
+                        v4f nx[4];
+    #pragma unroll
+                        for (int n = 0; n < 4; ++n) nx[n] = v4f{0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+                        for (int q = 0; q < 4; ++q)
+    #pragma unroll
+                            for (int n = 0; n < 4; ++n) nx[n] = mfma16x16x4(Am[n][q], acc[n][q], nx[n]);
+    #pragma unroll
+                        for (int n = 0; n < 4; ++n) acc[n] = nx[n];
+                    }
                 }
             } else {
 #pragma unroll
@@ -2302,7 +2580,12 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
                     const uint64_t bal = __ballot((posb >> tt) & 1u);
 #pragma unroll
                     for (int n = 0; n < 4; ++n)
-                        if (t0 + tt < pl[n]) acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
+                        if (t0 + tt < pl[n]) {
+                            if (WU && w.cs[n] + t0 + tt + 1 <= tw)
+                                acc[n] = mfma_step16_warm(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq, fr);
+                            else
+                                acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
+                        }
                 }
             }
         } else {
@@ -2310,7 +2593,12 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
                 const uint64_t bal = __ballot(ztilde_next(t) > 0.f);
 #pragma unroll
                 for (int n = 0; n < 4; ++n)
-                    if (t < pl[n]) acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
+                    if (t < pl[n]) {
+                        if (WU && w.cs[n] + t + 1 <= tw)
+                            acc[n] = mfma_step16_warm(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq, fr);
+                        else
+                            acc[n] = mfma_step16(acc[n], (uint32_t)(bal >> (16 * n)), g, WpD, Dq);
+                    }
             }
         }
     }
@@ -2327,11 +2615,24 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
                 if (rhs) gv[tt] = bload(rg, vg, 4 * (t0 + tt) * M);
                 else gv[tt] = forced ? seed_scale * (zv[tt] - xv[tt]) : 0.f;
             }
+            // latent warm-up: no MSE seed for rows k < tw; P_{k+1} = P_1 drops the observed
+            // latents' entries of J~_{k+1}^T lam for k + 1 <= tw
+            uint32_t kill = 0u;
+            if constexpr (WU) {
+                const uint32_t wr2 = low_bits(tw - (s0 + t0));   // bit tt: row s0 + t0 + tt < tw
+                if (!rhs) {
+#pragma unroll
+                    for (int tt = 0; tt < TB; ++tt) gv[tt] = ((wr2 >> tt) & 1u) ? 0.f : gv[tt];
+                }
+                kill = forced ? wr2 : 0u;   // same bits: s0 + t0 + tt + 1 <= tw
+            }
 #pragma unroll
             for (int tt = TB - 1; tt >= 0; --tt) {
                 const bool m = (posb >> tt) & 1u;
                 const float wt = row16_dot(wT, u);
-                const float y = (t0 + tt + 1 < len) ? pi * fmaf(Ai, u, m ? wt : 0.f) : 0.f;
+                bool on = t0 + tt + 1 < len;   // J~_{k+1}^T, P_{k+1} on the left
+                if constexpr (WU) on = on && !((kill >> tt) & 1u);
+                const float y = on ? pi * fmaf(Ai, u, m ? wt : 0.f) : 0.f;
                 if (lat) u = y + gv[tt];
             }
         } else {
@@ -2341,10 +2642,13 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
                 const float wt = row16_dot(wT, u);
                 if (run) {
                     const size_t step = (size_t)b * T + s0 + t;
-                    const float y = (t + 1 < len) ? pi * fmaf(Ai, u, m ? wt : 0.f) : 0.f;
+                    bool on = t + 1 < len;
+                    if constexpr (WU) on = on && !(forced && s0 + t + 1 <= tw);
+                    const float y = on ? pi * fmaf(Ai, u, m ? wt : 0.f) : 0.f;
                     float gk = 0.f;
                     if (rhs) gk = rhs[step * M + c];
-                    else if (forced) gk = seed_scale * (z[step * M + c] - x[((size_t)b * (T + 1) + s0 + t + 1) * N + c]);
+                    else if (forced && (!WU || s0 + t >= tw))
+                        gk = seed_scale * (z[step * M + c] - x[((size_t)b * (T + 1) + s0 + t + 1) * N + c]);
                     u = y + gk;
                 }
             }
@@ -2420,7 +2724,7 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn16_rev(
 // gradient partial sums dW[i][j] += lam_i relu(z~_j), dA_i += lam_i z~_i, dh_i += lam_i over
 // the wave's four chains (layout gpart[wave][16][18], the rotated dW columns put back).  A tile
 // row tt is step k = s0 + t0 + tt: z_k, x_k, x_{k+1}, g_k, and z_{k-1} for z~_k.
-template <int TB>
+template <int TB, bool WU>
 __global__ __launch_bounds__(64) void k_fixup_rev_plrnn16(const float *__restrict__ A, const float *__restrict__ W,
                                                          float alpha, int N, const float *__restrict__ gin,
                                                          float seed_scale, const float *__restrict__ x,
@@ -2428,7 +2732,8 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn16(const float *__restric
                                                          const float *__restrict__ carry_in,
                                                          const float *__restrict__ Pm, const float *__restrict__ vmap,
                                                          float *__restrict__ lam_out, float *__restrict__ gpart, int B,
-                                                         int T, int M, int C, int ncs) {
+                                                         int T, int M, int C, int ncs, int tw) {
+    static_assert(!WU || TB <= 16, "the warm-up variant runs 16-step tiles (bit masks of TB + 1 steps)");
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int nchains = B * ncs;
     const int chain0 = blockIdx.x * 4;
@@ -2475,7 +2780,7 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn16(const float *__restric
         if (s == 0) return z0 ? z0[(size_t)b * M + c] : (forced ? x[(size_t)b * (T + 1) * N + c] : 0.f);
         const float zp = z[((size_t)b * T + s - 1) * M + c];
         if (!forced) return zp;
-        return __fadd_rn(__fmul_rn(pi, zp), __fmul_rn(alpha, x[((size_t)b * (T + 1) + s) * N + c]));
+        return forced_in<WU>(pi, alpha, zp, x[((size_t)b * (T + 1) + s) * N + c], s, tw);
     };
     const int cl0 = min(chain0, nchains - 1);
     const int b0 = cl0 / ncs, s00 = (cl0 % ncs) * C;
@@ -2499,19 +2804,28 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn16(const float *__restric
                 gv[tt] = bload(rg, vg, 4 * (t0 + tt) * M);
             }
             xv[TB] = bload(rx, vx, 4 * (t0 + TB) * N);
-            // z~ of steps s0+t0 .. s0+t0+TB (the last only for the mask of the tile's top step)
+            // z~ of steps s0+t0 .. s0+t0+TB (the last only for the mask of the tile's top step);
+            // with a latent warm-up, bit j of wb marks step s0 + t0 + j <= tw (j <= TB <= 16)
+            uint32_t wb = 0u;
+            if constexpr (WU) wb = low_bits(tw - (s0 + t0) + 1);
             zt[0] = (len > 0 && lat) ? ztilde(s0 + t0) : 0.f;
 #pragma unroll
             for (int tt = 1; tt <= TB; ++tt)
-                zt[tt] = forced ? __fadd_rn(__fmul_rn(pi, zv[tt - 1]), __fmul_rn(alpha, xv[tt])) : zv[tt - 1];
+                zt[tt] = forced ? forced_at<WU>(pi, alpha, zv[tt - 1], xv[tt], wb, tt) : zv[tt - 1];
             if (!gin) {
 #pragma unroll
                 for (int tt = 0; tt < TB; ++tt) gv[tt] = forced ? seed_scale * (zv[tt] - xv[tt + 1]) : 0.f;
+                if constexpr (WU) {   // no MSE seed for the warm-up rows k < tw
+#pragma unroll
+                    for (int tt = 0; tt < TB; ++tt) gv[tt] = ((wb >> (tt + 1)) & 1u) ? 0.f : gv[tt];
+                }
             }
+            const uint32_t kill = forced ? (wb >> 1) : 0u;   // bit tt: P_{k+1} = P_1 (k + 1 <= tw)
 #pragma unroll
             for (int tt = TB - 1; tt >= 0; --tt) {
                 const int k = s0 + t0 + tt;
-                const bool nxt = k + 1 < T;
+                bool nxt = k + 1 < T;   // J~_{k+1}^T, P_{k+1} on the left
+                if constexpr (WU) nxt = nxt && !((kill >> tt) & 1u);
                 const bool m = zt[tt + 1] > 0.f;
                 const float wt = row16_dot(wT, lam);
                 const float y = nxt ? pi * fmaf(Ai, lam, m ? wt : 0.f) : 0.f;
@@ -2528,14 +2842,17 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn16(const float *__restric
                 const int k = s0 + t;
                 const bool nxt = run && k + 1 < T;
                 const bool m = nxt && ztilde(k + 1) > 0.f;
+                bool on = nxt;
+                if constexpr (WU) on = on && !(forced && k + 1 <= tw);
                 const float wt = row16_dot(wT, lam);
                 float zk = 0.f, lr = 0.f;
                 if (run) {
                     const size_t step = (size_t)b * T + k;
-                    const float y = nxt ? pi * fmaf(Ai, lam, m ? wt : 0.f) : 0.f;
+                    const float y = on ? pi * fmaf(Ai, lam, m ? wt : 0.f) : 0.f;
                     float gk = 0.f;
                     if (gin) gk = gin[step * M + c];
-                    else if (forced) gk = seed_scale * (z[step * M + c] - x[((size_t)b * (T + 1) + k + 1) * N + c]);
+                    else if (forced && (!WU || k >= tw))
+                        gk = seed_scale * (z[step * M + c] - x[((size_t)b * (T + 1) + k + 1) * N + c]);
                     lam = y + gk;
                     if (lam_out) lam_out[step * M + c] = lam;
                     zk = ztilde(k);
@@ -3203,7 +3520,7 @@ template <int MP>
 __global__ __launch_bounds__(256) void k_masks_plrnn(float alpha, int N, const float *__restrict__ x,
                                                      const float *__restrict__ z0, const float *__restrict__ z,
                                                      uint32_t *__restrict__ masks, const int *__restrict__ active,
-                                                     int B, int T, int M) {
+                                                     int B, int T, int M, int tw) {
     constexpr int NCH = 64 / MP, RQ = 8;
     const int lane = threadIdx.x & 63, n = lane / MP, i = lane % MP;
     const long total = (long)B * T;
@@ -3220,7 +3537,7 @@ __global__ __launch_bounds__(256) void k_masks_plrnn(float alpha, int N, const f
             int b = 0, s = 0;
             if (in) row_at(rb, rr, T, b, s);
             act[q] = in && (!active || active[b]);
-            zt[q] = (act[q] && i < M) ? forced_state(x, z0, z, b, s, i, T, M, N, alpha) : 0.f;
+            zt[q] = (act[q] && i < M) ? forced_state(x, z0, z, b, s, i, T, M, N, alpha, tw) : 0.f;
         }
 #pragma unroll
         for (int q = 0; q < RQ; ++q) {
@@ -3249,14 +3566,15 @@ int launch_resjac_plrnn(const PlrnnArgs &a, const float *z, float *F, float *r, 
         const int grid = (int)(want < 4096 ? want : 4096);
         KTimer kt("k_masks_plrnn", st);
         if (MP == 16)
-            hipLaunchKernelGGL(k_masks_plrnn<16>, dim3(grid), dim3(256), 0, st, a.alpha, a.N, a.x, a.z0, z, masks, active, a.B, a.T, a.M);
+            hipLaunchKernelGGL(k_masks_plrnn<16>, dim3(grid), dim3(256), 0, st, a.alpha, a.N, a.x, a.z0, z, masks, active, a.B, a.T, a.M, a.tw);
         else if (MP == 32)
-            hipLaunchKernelGGL(k_masks_plrnn<32>, dim3(grid), dim3(256), 0, st, a.alpha, a.N, a.x, a.z0, z, masks, active, a.B, a.T, a.M);
+            hipLaunchKernelGGL(k_masks_plrnn<32>, dim3(grid), dim3(256), 0, st, a.alpha, a.N, a.x, a.z0, z, masks, active, a.B, a.T, a.M, a.tw);
         else
-            hipLaunchKernelGGL(k_masks_plrnn<64>, dim3(grid), dim3(256), 0, st, a.alpha, a.N, a.x, a.z0, z, masks, active, a.B, a.T, a.M);
+            hipLaunchKernelGGL(k_masks_plrnn<64>, dim3(grid), dim3(256), 0, st, a.alpha, a.N, a.x, a.z0, z, masks, active, a.B, a.T, a.M, a.tw);
         DEER_LAUNCH_CHECK("k_masks_plrnn");
         return DEER_OK;
     }
+    if (a.tw > 0) return invalid_arg("the residual kernel takes no latent warm-up");
     const long groups = ((long)a.B * a.T + (64 / MP) - 1) / (64 / MP);
     const long passes = J ? groups : (groups + 3) / 4;
     const int grid = (int)(passes < 8192 ? passes : 8192);
@@ -3280,6 +3598,7 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+    if (a.tw > 0) return invalid_arg("the stored-mask chunk product takes no latent warm-up");
     KTimer kt("k_chunk_product_plrnn", st);
 #define CP(MPV, R)                                                                                                  \
     hipLaunchKernelGGL((k_chunk_product_plrnn<MPV, R>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, \
@@ -3309,19 +3628,29 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
     if (wmaps && (MP != 16 || ncs % 4))
         return invalid_arg("composed wave maps need M <= 16 and a chunk count divisible by 4");
     if (mark && MP != 16) return invalid_arg("pass marks are written by the M <= 16 forward pass only");
+    if (a.tw > 0 && MP != 16) return invalid_arg("the latent warm-up inside the Newton iteration needs M <= 16");
     if (MP == 64 && (a.N == 0 || a.N == a.M)) {   // uniform forcing factor: W-in-LDS kernel
         hipLaunchKernelGGL(k_newton_product_plrnn64u, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0,
                            z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
     } else if (MP == 16) {
 #define NP16(TBV, WPBV)                                                                                                \
-    hipLaunchKernelGGL((k_newton_product_plrnn16<TBV, WPBV>), dim3(grid / WPBV), dim3(64 * WPBV), 0, st, a.A, a.W, a.h, \
-                       a.alpha, a.N, a.x, a.z0, z, zalt, zsel, P, v, active, gamma, a.B, a.T, a.M, C, ncs, wmaps, gmap, \
-                       mark, pass_no)
+    hipLaunchKernelGGL((k_newton_product_plrnn16<TBV, WPBV, WUV>), dim3(grid / WPBV), dim3(64 * WPBV), 0, st, a.A, a.W, \
+                       a.h, a.alpha, a.N, a.x, a.z0, z, zalt, zsel, P, v, active, gamma, a.B, a.T, a.M, C, ncs, wmaps, \
+                       gmap, mark, pass_no, a.tw)
+#define NP16W(TBV, WPBV)            \
+    if (a.tw > 0) {                 \
+        constexpr bool WUV = true;  \
+        NP16(TBV, WPBV);            \
+    } else {                        \
+        constexpr bool WUV = false; \
+        NP16(TBV, WPBV);            \
+    }
         if (wmaps == 2) {
-            if (C % 32) NP16(16, 8); else NP16(32, 8);
+            if (C % 32) { NP16W(16, 8) } else { NP16W(32, 8) }
         } else {
-            if (C % 32) NP16(16, 1); else NP16(32, 1);
+            if (C % 32) { NP16W(16, 1) } else { NP16W(32, 1) }
         }
+#undef NP16W
 #undef NP16
     } else if (MP == 32) NP(32); else NP(64);
 #undef NP
@@ -3339,9 +3668,15 @@ int launch_newton_pass16(const PlrnnArgs &a, float *z, float *zalt, const float 
     KTimer kt("k_newton_pass16", st);
     const int grid = a.B * ncs / 32;
 #define NPS(TBV)                                                                                                  \
-    hipLaunchKernelGGL(k_newton_pass16<TBV>, dim3(grid), dim3(512), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, \
-                       z, zalt, a.T, a.M, C, ncs, Pin, vin, gin, Pout, vout, gout, fc, mark, pass_no)
-    if (C % 32) NPS(16); else NPS(32);
+    hipLaunchKernelGGL((k_newton_pass16<TBV, WUV>), dim3(grid), dim3(512), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x,  \
+                       a.z0, z, zalt, a.T, a.M, C, ncs, Pin, vin, gin, Pout, vout, gout, fc, mark, pass_no, a.tw)
+    if (a.tw > 0) {
+        constexpr bool WUV = true;
+        if (C % 32) NPS(16); else NPS(32);
+    } else {
+        constexpr bool WUV = false;
+        if (C % 32) NPS(16); else NPS(32);
+    }
 #undef NPS
     DEER_LAUNCH_CHECK("k_newton_pass16");
     return DEER_OK;
@@ -3447,16 +3782,24 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     hipLaunchKernelGGL(k_fixup_fwd_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, carry_in, \
                        z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
 #define FX16(TBV)                                                                                                 \
-    hipLaunchKernelGGL(k_fixup_fwd_plrnn16<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, \
-                       carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs, Pm, vm, gmap, fcv)
+    hipLaunchKernelGGL((k_fixup_fwd_plrnn16<TBV, WUV>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x,  \
+                       a.z0, carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs, Pm, vm, gmap, \
+                       fcv, a.tw)
     if (gmap && (!Pm || ncs % 32)) return invalid_arg("group maps need the wave maps and 32 | chunk count");
     if (Pm && (MP != 16 || ncs % 4))
         return invalid_arg("composed wave maps need M <= 16 and a chunk count divisible by 4");
     if (fc && MP != 16) return invalid_arg("the fused pass-end control needs M <= 16");
+    if (a.tw > 0 && MP != 16) return invalid_arg("the latent warm-up inside the Newton iteration needs M <= 16");
     FusedCtl fcv{};
     if (fc) fcv = *fc;
     if (MP == 16) {
-        if (C % 32) FX16(16); else FX16(32);
+        if (a.tw > 0) {
+            constexpr bool WUV = true;
+            if (C % 32) FX16(16); else FX16(32);
+        } else {
+            constexpr bool WUV = false;
+            if (C % 32) FX16(16); else FX16(32);
+        }
     } else if (fixup_mfma()) {
         const int gridm = (nch + 15) / 16;
 #define FXM(MPV, VV)                                                                                                 \
@@ -3481,6 +3824,7 @@ int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
+    if (a.tw > 0) return invalid_arg("the stored-mask reverse fix-up takes no latent warm-up");
     KTimer kt("k_fixup_rev_plrnn", st);
 #define FR(MPV)                                                                                                     \
     hipLaunchKernelGGL(k_fixup_rev_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, g,       \
@@ -3499,9 +3843,15 @@ int launch_adjoint_plrnn16(const PlrnnArgs &a, const float *g, float seed_scale,
     {
         KTimer kt("k_chunk_product_plrnn", st);
 #define CPR(TBV)                                                                                                     \
-    hipLaunchKernelGGL(k_chunk_product_plrnn16_rev<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, g, z, \
-                       a.x, seed_scale, P, v, a.B, a.T, a.M, C, ncs, (int)wm)
-        if (C % 32) CPR(16); else CPR(32);
+    hipLaunchKernelGGL((k_chunk_product_plrnn16_rev<TBV, WUV>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, \
+                       g, z, a.x, seed_scale, P, v, a.B, a.T, a.M, C, ncs, (int)wm, a.tw)
+        if (a.tw > 0) {   // 16-step tiles: the warm-up variant's registers fit two waves per SIMD
+            constexpr bool WUV = true;
+            CPR(16);
+        } else {
+            constexpr bool WUV = false;
+            if (C % 32) CPR(16); else CPR(32);
+        }
 #undef CPR
         DEER_LAUNCH_CHECK("k_chunk_product_plrnn16_rev");
     }
@@ -3512,9 +3862,16 @@ int launch_adjoint_plrnn16(const PlrnnArgs &a, const float *g, float seed_scale,
     {
         KTimer kt("k_fixup_rev_plrnn", st);
 #define FRV(TBV)                                                                                                   \
-    hipLaunchKernelGGL(k_fixup_rev_plrnn16<TBV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, g, seed_scale, \
-                       a.x, a.z0, z, carry, wm ? P : nullptr, wm ? v : nullptr, lam, gpart, a.B, a.T, a.M, C, ncs)
-        if (C % 32) FRV(16); else FRV(32);
+    hipLaunchKernelGGL((k_fixup_rev_plrnn16<TBV, WUV>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, g,       \
+                       seed_scale, a.x, a.z0, z, carry, wm ? P : nullptr, wm ? v : nullptr, lam, gpart, a.B, a.T, a.M, C, \
+                       ncs, a.tw)
+        if (a.tw > 0) {
+            constexpr bool WUV = true;
+            FRV(16);
+        } else {
+            constexpr bool WUV = false;
+            if (C % 32) FRV(16); else FRV(32);
+        }
 #undef FRV
         DEER_LAUNCH_CHECK("k_fixup_rev_plrnn16");
     }

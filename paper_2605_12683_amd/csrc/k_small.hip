@@ -524,6 +524,10 @@ __global__ __launch_bounds__(SNT) void k_adjoint_small(const float *__restrict__
 bool newton_small_fits(int M, int T, int fixed_iters) { return M <= SMS && T <= SNT * SC && fixed_iters > 0; }
 
 int launch_newton_small(const PlrnnArgs &a, float *z, int iters, uint32_t *norm_bits, hipStream_t st) {
+    if (a.tw > 0) {
+        set_error("the one-launch solve takes no latent warm-up");
+        return DEER_ERR_INVALID_ARG;
+    }
     const int nc = (a.T + SC - 1) / SC;
     KTimer kt("k_newton_small", st);
     hipLaunchKernelGGL(k_newton_small, dim3(a.B), dim3(SNT), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, z, a.T, a.M,
@@ -539,6 +543,10 @@ bool adjoint_small_fits(int M, int T) { return M <= SMS && T <= SNT * SC; }
 
 int launch_adjoint_small(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *lam,
                          float *gpart, float *dA, float *dW, float *dh, hipStream_t st) {
+    if (a.tw > 0) {
+        set_error("the one-launch adjoint takes no latent warm-up");
+        return DEER_ERR_INVALID_ARG;
+    }
     const int nc = (a.T + SC - 1) / SC;
     KTimer kt("k_adjoint_small", st);
     hipLaunchKernelGGL(k_adjoint_small, dim3(a.B), dim3(SNT), 0, st, a.A, a.W, a.alpha, a.N, a.x, a.z0, z, g,

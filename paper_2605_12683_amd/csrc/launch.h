@@ -12,6 +12,9 @@ struct PlrnnArgs {
     int N;
     const float *x, *z0;
     int B, T, M;
+    // latent warm-up inside the Newton iteration (M <= 16 kernels and the mask pass): the forced
+    // inputs of steps 1..tw take alpha = 1 and their Jacobians P_1; 0 = none
+    int tw = 0;
 };
 
 struct ShArgs {

@@ -45,3 +45,13 @@ def test_update_rows_counts_each_update_over_its_part():
     assert bench.update_rows(1000, 100, 26, 3, 2) < 26 * 1000
     with pytest.raises(ValueError):
         bench.update_rows(1000, 100, 5, 3, 2)
+
+
+def test_warmup_in_one_iteration_where_the_library_takes_it():
+    # vanilla PLRNN M <= 16 (GTF-DEER): one iteration, every update over all T steps
+    assert bench.warmup_in_one_iteration("plrnn", 16, False)
+    assert bench.warmup_in_one_iteration("plrnn", 3, False)
+    # chained solves elsewhere
+    assert not bench.warmup_in_one_iteration("plrnn", 17, False)
+    assert not bench.warmup_in_one_iteration("plrnn", 16, True)
+    assert not bench.warmup_in_one_iteration("shplrnn", 16, False)

@@ -2,12 +2,14 @@
 left out of the loss) against the float64 oracle: solves against the warm-up rollout, adjoints
 and gradients against the oracle's recursion at the same float32 trajectory, for GTF-DEER and
 quasi-DEER, vanilla and shallow PLRNNs."""
+import os
+
 import numpy as np
 import pytest
 
 import oracle as O
 import workloads as W
-from gpu_util import oracle_model, rel_inf, say
+from gpu_util import masks_to_bool, oracle_model, rel_inf, say
 
 pytestmark = pytest.mark.gpu
 
@@ -18,6 +20,16 @@ if not torch.cuda.is_available():
 import paper_2605_12683_amd as D  # noqa: E402
 
 TOL = 1e-4
+_ENV = ("DEER_CHUNK", "DEER_GROUP_MAPS", "DEER_PASS_FUSION")
+
+
+@pytest.fixture(autouse=True)
+def _no_overrides():
+    for k in _ENV:
+        os.environ.pop(k, None)
+    yield
+    for k in _ENV:
+        os.environ.pop(k, None)
 CASES = [("plrnn", 16, 0, 3, 2, 700, 100), ("plrnn", 3, 0, 3, 1, 300, 1), ("plrnn", 24, 0, 24, 3, 1000, 999),
          ("plrnn", 64, 0, 64, 2, 513, 200), ("shplrnn", 5, 50, 3, 2, 600, 128), ("shplrnn", 32, 256, 32, 1, 800, 50)]
 
@@ -68,3 +80,67 @@ def test_warmup_with_given_cotangent_and_initial_state():
     gr = O.param_grads(m, c.x, z32, c.alpha, 2, lam, z0=z0, mask_precision="float32", T_w=T_w)
     for k, v in out["grads"].items():
         assert rel_inf(v.cpu().numpy(), gr[k]) < TOL, k
+
+
+# M <= 16: the warm-up is part of the one Newton iteration (the register-tiled kernels take the
+# forcing strength per step: alpha_s = 1 and P_1 for s <= T_w).  T_w at the first step, inside a
+# chunk and a tile, on a chunk boundary (T_w + 1 divisible by the chunk length) and next to the
+# end; chunk layouts through the per-step slow paths (ragged tiles), composed wave maps, group
+# maps and the fused pass kernel; every latent observed; M = 3 (the one-launch kernels step aside).
+JOINT = [(16, 3, 2, 700, 100, 0), (16, 3, 2, 2048, 511, 16), (16, 3, 2, 2048, 700, 16), (12, 4, 2, 4096, 1, 32),
+         (12, 4, 2, 4096, 4094, 32), (7, 3, 3, 640, 77, 40), (5, 2, 3, 1000, 333, 25), (16, 16, 2, 513, 200, 0),
+         (3, 3, 1, 300, 17, 0)]
+
+
+def _joint_case(M, N, B, T, T_w, chunk, seed):
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    os.environ["DEER_GROUP_MAPS"] = "1"   # where 32 divides the chunk count, whatever the size
+    return W.random_plrnn_case(M, N, B, T, 0.2, seed, w_norm=0.2, a_range=(0.3, 0.75))
+
+
+@pytest.mark.parametrize("M,N,B,T,T_w,chunk", JOINT)
+def test_warmup_one_iteration_newton_iterates(M, N, B, T, T_w, chunk):
+    """The k-th Newton iterate of the joint iteration equals the oracle's (Alg. GTF-DEER with
+    P_1 for t <= T_w), for k = 1 and 3: the per-step forcing in the residual, the chunk products,
+    the local solutions and the fix-up."""
+    c = _joint_case(M, N, B, T, T_w, chunk, 4100 + M + T_w)
+    m = oracle_model(c)
+    for k in (1, 3):
+        say("warm-up one iteration, fixed updates", M, N, B, T, T_w, chunk, k)
+        res = D.deer_solve(m, c.x, c.alpha, N, fixed_iters=k, T_w=T_w, want_masks=True)
+        ref = O.newton(m, c.x, c.alpha, N, fixed_iters=k, T_w=T_w)
+        assert res["status"] == 0 and res["iters"] == [k] * B
+        z = res["z"].cpu().numpy()
+        assert rel_inf(z, ref["z"]) < TOL, k
+        fp32 = O.activation_mask_fp32(m, z, c.x, c.alpha, N, None, T_w)
+        assert np.array_equal(masks_to_bool(res["masks"].cpu().numpy(), M), fp32)
+
+
+@pytest.mark.parametrize("M,N,B,T,T_w,chunk", JOINT)
+def test_warmup_one_iteration_counts_and_adjoint(M, N, B, T, T_w, chunk):
+    """Solved to tolerance the joint iteration reaches the warm-up rollout in the oracle's number
+    of updates (up to one), with the fused pass kernel and with separate kernels; the adjoint
+    and gradients (MSE over the states after the warm-up, and a given cotangent) match the
+    oracle's joint recursion."""
+    c = _joint_case(M, N, B, T, T_w, chunk, 4200 + M + T_w)
+    m = oracle_model(c)
+    ref = O.rollout(m, c.x, c.alpha, N, T_w=T_w)
+    want = O.newton(m, c.x, c.alpha, N, tol=1e-5, T_w=T_w)["iters"].tolist()
+    for fuse in ("1", "0"):
+        os.environ["DEER_PASS_FUSION"] = fuse
+        say("warm-up one iteration to tolerance", M, N, B, T, T_w, chunk, fuse)
+        res = D.deer_solve(m, c.x, c.alpha, N, tol=1e-5, max_iter=200, T_w=T_w)
+        assert res["status"] == 0, res
+        assert rel_inf(res["z"].cpu().numpy(), ref) < TOL
+        assert max(abs(a - b) for a, b in zip(res["iters"], want)) <= 1, (res["iters"], want)
+    z32 = ref.astype(np.float32)
+    g = np.random.default_rng(M + T_w).standard_normal(z32.shape).astype(np.float32)
+    for gg in (None, g):
+        say("warm-up one iteration adjoint", M, N, B, T, T_w, chunk, gg is None)
+        out = D.deer_adjoint(m, c.x, z32, c.alpha, N, g=gg, T_w=T_w)
+        lam = O.adjoint(m, c.x, z32, c.alpha, N, g=gg, mask_precision="float32", T_w=T_w)
+        assert rel_inf(out["lam"].cpu().numpy(), lam) < TOL
+        gr = O.param_grads(m, c.x, z32, c.alpha, N, lam, mask_precision="float32", T_w=T_w)
+        for k, v in out["grads"].items():
+            assert rel_inf(v.cpu().numpy(), gr[k]) < TOL, k

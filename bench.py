@@ -60,9 +60,10 @@ def _plrnn_step(D, model, xd, c, ws_s, ws_a, T_w=0):
 
 
 def warmup_in_one_iteration(kind, M, quasi):
-    """The library runs the latent warm-up inside the one Newton iteration for the vanilla PLRNN
-    with M <= 16 (GTF-DEER, identity read-out); elsewhere it chains two solves."""
-    return kind == "plrnn" and M <= 16 and not quasi
+    """The library runs the latent warm-up inside the one Newton iteration for GTF-DEER on the
+    vanilla PLRNN with M <= 16 and on the shallow PLRNN (identity read-out); elsewhere it chains
+    two solves."""
+    return not quasi and ((kind == "plrnn" and M <= 16) or kind == "shplrnn")
 
 
 def update_rows(T, T_w, updates, warm_updates, nsteps):

@@ -862,11 +862,29 @@ static int init_guess(const deer_solve_opts *o, int B, int T, int M, int N, cons
     return DEER_OK;
 }
 
-// The latent warm-up inside the one Newton iteration (per-step forcing strength in the kernels):
-// the register-tiled vanilla PLRNN path (M <= 16) with the identity read-out.  The other paths
-// solve the warm-up prefix and the rest as two chained problems (solve_warmup below).
+// The latent warm-up inside the one Newton iteration (per-step forcing strength in the kernels),
+// identity read-out: the register-tiled vanilla PLRNN path (M <= 16) and the shallow PLRNN.  The
+// other paths solve the warm-up prefix and the rest as two chained problems (solve_warmup below).
 static bool warmup_joint(const deer_model *m, const deer_forcing *f) {
-    return f->T_w > 0 && !f->obs && m->kind == DEER_PLRNN && m->M <= 16;
+    return f->T_w > 0 && !f->obs && ((m->kind == DEER_PLRNN && m->M <= 16) || m->kind == DEER_SHPLRNN);
+}
+
+// J~ of every step of the shallow model into J; with a latent warm-up, steps 0..T_w take P_1
+// (alpha = 1; step 0's Jacobian only multiplies the fixed initial state's zero update) and the
+// rest P_alpha
+static int jacform_sh(const ShArgs &a, const uint32_t *masks, float *J, const int *active, const float *gamma,
+                      hipStream_t st) {
+    if (a.tw <= 0) return launch_jacform_shplrnn(a, masks, J, active, gamma, st);
+    ShArgs w = a;
+    w.alpha = 1.f;
+    w.t_lo = 0;
+    w.t_hi = a.tw + 1;
+    int rc = launch_jacform_shplrnn(w, masks, J, active, gamma, st);
+    if (rc || a.tw + 1 >= a.T) return rc;
+    w.alpha = a.alpha;
+    w.t_lo = a.tw + 1;
+    w.t_hi = a.T;
+    return launch_jacform_shplrnn(w, masks, J, active, gamma, st);
 }
 
 static int solve_plrnn(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
@@ -953,6 +971,7 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
     if ((rc = check_ws(ws, ws_bytes, need))) return rc;
     ShWs w = carve_sh(ws, B, T, m->M, m->L, DEER_OP_SOLVE, false, false, &need, !fused);
     ShArgs a{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
+    a.tw = f->T_w;
     if ((rc = init_guess(o, B, T, m->M, f->n_forced, x, z, st))) return rc;
     std::vector<int> act(B, 1), it(B, 0);
     std::vector<float> norm(B, NAN);
@@ -973,7 +992,7 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
             return launch_fixup_shjvp(false, a, w.masks, w.r, -1.f, gam, d.carry, zb, za, zsel, w.ctl.chain_bits, dact,
                                       d.C, d.ncs, st);
         }
-        if ((r = launch_jacform_shplrnn(a, w.masks, w.J, dact, gam, st))) return r;
+        if ((r = jacform_sh(a, w.masks, w.J, dact, gam, st))) return r;
         if ((r = launch_chunk_product_dense(false, B, T, m->M, w.J, w.r, -1.f, d.P, d.v, dact, d.C, d.ncs, st))) return r;
         if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nullptr, B, d.ncs, d.gws, st))) return r;
         return launch_fixup_dense(0, B, T, m->M, w.J, w.r, -1.f, d.carry, zb, za, zsel, w.ctl.chain_bits, dact, d.C,
@@ -1659,11 +1678,12 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
         if ((rc = check_ws(ws, ws_bytes, need))) return rc;
         ShWs w = carve_sh(ws, B, T, m->M, m->L, DEER_OP_ADJOINT, true, true, &need, !fused);
         ShArgs a{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
+        a.tw = f->T_w;
         const DenseWs &d = w.d;
         const float *gg = g;
-        if (!gg) {
-            const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
-            if ((rc = launch_mse_seed(z, x, scale, B, T, m->M, f->n_forced, w.g, st))) return rc;
+        if (!gg) {   // MSE over the states after the warm-up, z_{T_w+1}..z_T
+            const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * (T - f->T_w))) : 0.f;
+            if ((rc = launch_mse_seed(z, x, scale, B, T, m->M, f->n_forced, w.g, st, f->T_w))) return rc;
             gg = w.g;
         }
         float *lo = lam ? lam : w.lam;
@@ -1677,7 +1697,7 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
                                          nullptr, d.C, d.ncs, st)))
                 return rc;
         } else {
-            if ((rc = launch_jacform_shplrnn(a, w.masks, w.J, nullptr, nullptr, st))) return rc;
+            if ((rc = jacform_sh(a, w.masks, w.J, nullptr, nullptr, st))) return rc;
             if ((rc = launch_chunk_product_dense(true, B, T, m->M, w.J, gg, 1.f, d.P, d.v, nullptr, d.C, d.ncs, st)))
                 return rc;
             if ((rc = launch_carry(d.MP, true, d.P, d.v, d.carry, nullptr, nullptr, B, d.ncs, d.gws, st))) return rc;

@@ -229,8 +229,10 @@ __device__ __forceinline__ float big_forced(const ShArgs &a, const float *z, int
     if (a.zt) return a.zt[((size_t)b * a.T + s) * a.M + i];
     const float zp = z[((size_t)b * a.T + s - 1) * a.M + i];
     if (i >= a.N) return zp;
+    const float xs = a.x[((size_t)b * (a.T + 1) + s) * a.N + i];
+    if (s <= a.tw) return xs;   // latent warm-up: alpha_s = 1
     const float p = __fsub_rn(1.0f, a.alpha);
-    return __fadd_rn(__fmul_rn(p, zp), __fmul_rn(a.alpha, a.x[((size_t)b * (a.T + 1) + s) * a.N + i]));
+    return __fadd_rn(__fmul_rn(p, zp), __fmul_rn(a.alpha, xs));
 }
 
 // LDS: W1 [M][L] | W2 [L][M] | z~ [BG] | relu(u) [L]

@@ -64,12 +64,14 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
     const int rc = tid / (MP / 4), i0 = 4 * (tid % (MP / 4));
     float pz[4], px[4], pc[4], cz[4];   // z_{s-1} (or the initial state at s = 0), x_s, z_s
     bool plater = false;                // the fetched row exists and has s > 0
+    bool pwarm = false;                 // ... and is a latent warm-up step (s <= tw: z~ = x)
     auto fetch = [&](long tile) {
         const long row = tile * TT + rc;
         const bool ok = tid < NT4 && tile < ntiles && row < total;
         int b = 0, s = 0;
         if (ok) row_at(row_base(tile * TT, T), rc, T, b, s);
         plater = ok && s > 0;
+        pwarm = plater && s <= a.tw;
         const float *z = cur_iter(zbuf, zalt, zsel, b);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -106,12 +108,12 @@ __global__ __launch_bounds__(256) void k_resjac_shplrnn(const ShArgs a, const fl
         const long row0 = tile * TT;
         __syncthreads();   // the previous tile is done with zT, zc, ru and red
         if (tid < NT4) {
-            const bool later = plater;
+            const bool later = plater, warm = pwarm;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int i = i0 + r;
                 float zt = pz[r];
-                if (later && i < N) zt = __fadd_rn(__fmul_rn(p, pz[r]), __fmul_rn(a.alpha, px[r]));
+                if (later && i < N) zt = warm ? px[r] : __fadd_rn(__fmul_rn(p, pz[r]), __fmul_rn(a.alpha, px[r]));
                 zT[i * TT + rc] = zt;
                 cz[r] = pc[r];
             }
@@ -372,7 +374,8 @@ __global__ __launch_bounds__(SHG_THREADS) void k_grads_shplrnn(const ShArgs a, c
             float vz = 0.f, vl = 0.f;
             if (row < total && i < M) {
                 const int b = (int)(row / T), s = (int)(row % T);
-                vz = (a.zt && s > 0) ? a.zt[(size_t)row * M + i] : forced_state(a.x, a.z0, z, b, s, i, T, M, a.N, a.alpha);
+                vz = (a.zt && s > 0) ? a.zt[(size_t)row * M + i]
+                                     : forced_state(a.x, a.z0, z, b, s, i, T, M, a.N, a.alpha, a.tw);
                 vl = lam[(size_t)row * M + i];
             }
             zt[tt][i] = vz;
@@ -452,15 +455,16 @@ __global__ void k_reduce_rows(const float *__restrict__ part, int nrows, int wid
     }
 }
 
-// MSE seed g_t = scale * [z_t[:N] - x_t; 0] (used by the stored-Jacobian adjoint)
+// MSE seed g_t = scale * [z_t[:N] - x_t; 0] (used by the stored-Jacobian adjoint); rows s < tw
+// (the latent warm-up's states z_1..z_tw) are left out of the loss
 __global__ void k_mse_seed(const float *__restrict__ z, const float *__restrict__ x, float scale, int B, int T, int M,
-                           int N, float *__restrict__ g) {
+                           int N, float *__restrict__ g, int tw) {
     const size_t n = (size_t)B * T * M;
     for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n; e += (size_t)gridDim.x * blockDim.x) {
         const int i = (int)(e % M);
         const size_t bt = e / M;
         const int b = (int)(bt / T), s = (int)(bt % T);
-        g[e] = i < N ? scale * (z[e] - x[((size_t)b * (T + 1) + s + 1) * N + i]) : 0.f;
+        g[e] = (i < N && s >= tw) ? scale * (z[e] - x[((size_t)b * (T + 1) + s + 1) * N + i]) : 0.f;
     }
 }
 
@@ -545,11 +549,12 @@ int launch_grads_shplrnn(const ShArgs &a, const float *z, const float *lam, cons
     return DEER_OK;
 }
 
-int launch_mse_seed(const float *z, const float *x, float scale, int B, int T, int M, int N, float *g, hipStream_t st) {
+int launch_mse_seed(const float *z, const float *x, float scale, int B, int T, int M, int N, float *g, hipStream_t st,
+                    int tw) {
     const size_t n = (size_t)B * T * M;
     const int grid = (int)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
     KTimer kt("k_mse_seed", st);
-    hipLaunchKernelGGL(k_mse_seed, dim3(grid), dim3(256), 0, st, z, x, scale, B, T, M, N, g);
+    hipLaunchKernelGGL(k_mse_seed, dim3(grid), dim3(256), 0, st, z, x, scale, B, T, M, N, g, tw);
     DEER_LAUNCH_CHECK("k_mse_seed");
     return DEER_OK;
 }

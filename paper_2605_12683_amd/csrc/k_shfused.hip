@@ -154,6 +154,20 @@ __device__ __forceinline__ void shf_afrag(const v4f (&jt)[MP / 16][MP / 16], con
             }
 }
 
+// a latent warm-up step's P_1 (section "Latent state warm-up"): the observed latents' columns of
+// J~ (k-steps 16 j + 4 g + q < N) dropped from its A fragments
+template <int MP>
+__device__ __forceinline__ void shf_drop_observed(float (&ac)[MP / 16][MP / 4], int N, int g) {
+    constexpr int NI = MP / 16;
+#pragma unroll
+    for (int I = 0; I < NI; ++I)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (16 * j + 4 * g + q < N) ac[I][4 * j + q] = 0.f;
+}
+
 // ---------------------------------------------------------------------------------------
 // forward chunk product: per chain the B operand is [P | u] (P's MP/16 column tiles plus one
 // whose column 0 is u), P <- J~_t P and u <- J~_t u + rhs_sign r_t, with P = I and u = 0 at
@@ -220,6 +234,7 @@ __global__ __launch_bounds__(256) void k_chunk_product_shfused(const ShArgs a, c
             if (nt >= nv) break;
             float ac[NI][NS];
             shf_afrag<MP>(jt[nt], dg, gm, g, c, ac);
+            if (a.tw > 0 && s0 + t0 + nt <= a.tw) shf_drop_observed<MP>(ac, N, g);
 #pragma unroll
             for (int tt = 0; tt <= PT; ++tt) {
                 float Bop[NS];
@@ -336,6 +351,7 @@ __global__ __launch_bounds__(256) void k_chunk_product_shfused_rev(const ShArgs 
             if (nt >= nj) continue;
             float ac[NI][NS];
             shf_afrag<MP>(jt[nt], dg, 1.f, g, c, ac);
+            if (a.tw > 0 && s0 + t0 + nt + 1 <= a.tw) shf_drop_observed<MP>(ac, N, g);   // J~_{k+1}
 #pragma unroll
             for (int tt = 0; tt < PT; ++tt) {
                 float Bop[NS];
@@ -491,6 +507,17 @@ __global__ __launch_bounds__(256) void k_fixup_shjvp(const ShArgs a, const uint3
         const int kcur = krow(t);
         // the Jacobian term of this step: always forward; reverse unless k + 1 = T
         const bool hasj = !REV || kcur + 1 < T;
+        // latent warm-up step of this lane's chain (P_1 in J~_k, forward, or J~_{k+1}, reverse):
+        // the observed latents' entries of y enter neither W2 diag(p) y nor the diagonal term
+        // (forward), or the output's observed rows vanish (reverse)
+        const bool wdrop = a.tw > 0 && (REV ? kcur + 1 : kcur) <= a.tw && t < len;
+        if (!REV && a.tw > 0) {
+#pragma unroll
+            for (int I = 0; I < NI; ++I)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (wdrop && 16 * I + 4 * g + r < N) dl[I][r] = 0.f;
+        }
         fetch(t + 1);
         v4f u[NLW];
 #pragma unroll
@@ -520,7 +547,8 @@ __global__ __launch_bounds__(256) void k_fixup_shjvp(const ShArgs a, const uint3
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const bool own = r == wv;
-                const float jv = hasj ? gm * (own ? fmaf(dg[I][r], dl[I][r], p2[I][r]) : p2[I][r]) : 0.f;
+                const bool jon = hasj && !(REV && wdrop && 16 * I + 4 * g + r < N);
+                const float jv = jon ? gm * (own ? fmaf(dg[I][r], dl[I][r], p2[I][r]) : p2[I][r]) : 0.f;
                 ct[r] = own ? fmaf(rhs_sign, rcur[I], jv) : jv;
             }
             red[buf][wv][I][lane] = ct;
@@ -705,6 +733,8 @@ __global__ __launch_bounds__(256) void k_resjac_shmfma(const ShArgs a, const flo
                 float v;
                 if (s == 0)   // the initial state: z0, or [x_0; 0]
                     v = a.z0 ? cur.zp[j][q] : (i < N ? cur.xs[j][q] : 0.f);
+                else if (i < N && s <= a.tw)   // latent warm-up: alpha_s = 1
+                    v = cur.xs[j][q];
                 else
                     v = i < N ? __fadd_rn(__fmul_rn(p, cur.zp[j][q]), __fmul_rn(a.alpha, cur.xs[j][q])) : cur.zp[j][q];
                 const bool e = rok && i < M;

@@ -32,6 +32,10 @@ struct ShArgs {
     const float *zt = nullptr;
     const float *Cd = nullptr;
     int t_lo = 0, t_hi = 0;
+    // latent warm-up inside the Newton iteration (identity read-out): the forced inputs of steps
+    // 1..tw take alpha = 1 and the Jacobians of those steps P_1; 0 = none.  The stored-Jacobian
+    // formation takes the warm-up as a separate step range with alpha = 1 instead.
+    int tw = 0;
 };
 
 int padded_dim(int M);
@@ -208,7 +212,9 @@ int launch_jacform_shplrnn(const ShArgs &a, const uint32_t *masks, float *J, con
                            hipStream_t st);
 int launch_grads_shplrnn(const ShArgs &a, const float *z, const float *lam, const uint32_t *masks, float *part,
                          const deer_grads *gr, hipStream_t st);
-int launch_mse_seed(const float *z, const float *x, float scale, int B, int T, int M, int N, float *g, hipStream_t st);
+// rows s < tw (the latent warm-up's states) get no seed
+int launch_mse_seed(const float *z, const float *x, float scale, int B, int T, int M, int N, float *g, hipStream_t st,
+                    int tw = 0);
 
 // read-out MLP of the diagonal SSM
 struct RoArgs {

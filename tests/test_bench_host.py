@@ -54,4 +54,5 @@ def test_warmup_in_one_iteration_where_the_library_takes_it():
     # chained solves elsewhere
     assert not bench.warmup_in_one_iteration("plrnn", 17, False)
     assert not bench.warmup_in_one_iteration("plrnn", 16, True)
-    assert not bench.warmup_in_one_iteration("shplrnn", 16, False)
+    assert bench.warmup_in_one_iteration("shplrnn", 64, False)
+    assert not bench.warmup_in_one_iteration("shplrnn", 16, True)

@@ -20,7 +20,7 @@ if not torch.cuda.is_available():
 import paper_2605_12683_amd as D  # noqa: E402
 
 TOL = 1e-4
-_ENV = ("DEER_CHUNK", "DEER_GROUP_MAPS", "DEER_PASS_FUSION")
+_ENV = ("DEER_CHUNK", "DEER_GROUP_MAPS", "DEER_PASS_FUSION", "DEER_SH_FUSED", "DEER_SH_RESMFMA")
 
 
 @pytest.fixture(autouse=True)
@@ -144,3 +144,52 @@ def test_warmup_one_iteration_counts_and_adjoint(M, N, B, T, T_w, chunk):
         gr = O.param_grads(m, c.x, z32, c.alpha, N, lam, mask_precision="float32", T_w=T_w)
         for k, v in out["grads"].items():
             assert rel_inf(v.cpu().numpy(), gr[k]) < TOL, k
+
+
+# Shallow PLRNN: the warm-up inside the one Newton iteration on every path: the Jacobians rebuilt
+# from the masks (P_1 in the warm-up steps of the chunk products and Jacobian-vector fix-ups) with
+# the matrix-core or the fixed-order residual, the stored Jacobians (formed per step range), and
+# M > 64 (the wide kernels).  Cases: (M, L, N, B, T, T_w, chunk, check the 1st and 2nd iterates).
+SH_JOINT = [(5, 50, 3, 2, 600, 128, 0, True), (32, 256, 32, 1, 800, 50, 0, False),
+            (20, 40, 5, 3, 300, 77, 64, True), (16, 64, 16, 2, 500, 1, 0, True),
+            (64, 128, 64, 1, 300, 150, 0, True), (100, 64, 20, 1, 200, 60, 0, True)]
+SH_PATHS = {"stored": ("0", "1"), "fixed-order residual": ("1", "0"), "matrix-core residual": ("1", "1")}
+
+
+@pytest.mark.parametrize("M,L,N,B,T,T_w,chunk,iterates", SH_JOINT)
+def test_shallow_warmup_one_iteration(M, L, N, B, T, T_w, chunk, iterates):
+    """The oracle's joint iteration (Alg. GTF-DEER with P_1 for t <= T_w): its first Newton
+    iterates, its update counts (up to one) and its fixed point, then the adjoint and the
+    gradients, on every shallow path."""
+    if chunk:
+        os.environ["DEER_CHUNK"] = str(chunk)
+    c = W.random_shplrnn_case(M, L, N, B, T, 0.15, 4300 + M + T_w, w_norm=0.2, a_range=(0.3, 0.75))
+    m = oracle_model(c)
+    ref = O.rollout(m, c.x, c.alpha, N, T_w=T_w)
+    want = O.newton(m, c.x, c.alpha, N, tol=1e-5, T_w=T_w)["iters"].tolist()
+    firsts = {k: O.newton(m, c.x, c.alpha, N, fixed_iters=k, T_w=T_w)["z"] for k in (1, 2)} if iterates else {}
+    z32 = ref.astype(np.float32)
+    lam = O.adjoint(m, c.x, z32, c.alpha, N, mask_precision="float32", T_w=T_w)
+    gr = O.param_grads(m, c.x, z32, c.alpha, N, lam, mask_precision="float32", T_w=T_w)
+    try:
+        for path, (fz, rm) in SH_PATHS.items():
+            os.environ["DEER_SH_FUSED"] = fz
+            os.environ["DEER_SH_RESMFMA"] = rm
+            for k, zk in firsts.items():
+                say("shallow warm-up one iteration, fixed updates", path, M, L, N, B, T, T_w, k)
+                res = D.deer_solve(m, c.x, c.alpha, N, fixed_iters=k, T_w=T_w)
+                assert res["status"] == 0 and res["iters"] == [k] * B
+                assert rel_inf(res["z"].cpu().numpy(), zk) < TOL, (path, k)
+            say("shallow warm-up one iteration to tolerance", path, M, L, N, B, T, T_w)
+            res = D.deer_solve(m, c.x, c.alpha, N, tol=1e-5, max_iter=200, T_w=T_w)
+            assert res["status"] == 0, (path, res)
+            assert rel_inf(res["z"].cpu().numpy(), ref) < TOL, path
+            assert max(abs(a - b) for a, b in zip(res["iters"], want)) <= 1, (path, res["iters"], want)
+            say("shallow warm-up one iteration adjoint", path)
+            out = D.deer_adjoint(m, c.x, z32, c.alpha, N, T_w=T_w)
+            assert rel_inf(out["lam"].cpu().numpy(), lam) < TOL, path
+            for key, v in out["grads"].items():
+                assert rel_inf(v.cpu().numpy(), gr[key]) < TOL, (path, key)
+    finally:
+        os.environ.pop("DEER_SH_FUSED", None)
+        os.environ.pop("DEER_SH_RESMFMA", None)

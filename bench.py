@@ -60,10 +60,9 @@ def _plrnn_step(D, model, xd, c, ws_s, ws_a, T_w=0):
 
 
 def warmup_in_one_iteration(kind, M, quasi):
-    """The library runs the latent warm-up inside the one Newton iteration for GTF-DEER on the
-    vanilla PLRNN with M <= 16 and on the shallow PLRNN (identity read-out); elsewhere it chains
-    two solves."""
-    return not quasi and ((kind == "plrnn" and M <= 16) or kind == "shplrnn")
+    """The library runs the latent warm-up inside the one Newton iteration for GTF-DEER on both
+    PLRNN kinds (identity read-out); quasi-DEER chains two solves."""
+    return not quasi and kind in ("plrnn", "shplrnn")
 
 
 def update_rows(T, T_w, updates, warm_updates, nsteps):

@@ -862,11 +862,11 @@ static int init_guess(const deer_solve_opts *o, int B, int T, int M, int N, cons
     return DEER_OK;
 }
 
-// The latent warm-up inside the one Newton iteration (per-step forcing strength in the kernels),
-// identity read-out: the register-tiled vanilla PLRNN path (M <= 16) and the shallow PLRNN.  The
-// other paths solve the warm-up prefix and the rest as two chained problems (solve_warmup below).
+// The latent warm-up inside the one Newton iteration (per-step forcing strength in the kernels):
+// GTF-DEER with the identity read-out, both PLRNN kinds.  Quasi-DEER solves the warm-up prefix
+// and the rest as two chained problems (solve_warmup below).
 static bool warmup_joint(const deer_model *m, const deer_forcing *f) {
-    return f->T_w > 0 && !f->obs && ((m->kind == DEER_PLRNN && m->M <= 16) || m->kind == DEER_SHPLRNN);
+    return f->T_w > 0 && !f->obs && (m->kind == DEER_PLRNN || m->kind == DEER_SHPLRNN);
 }
 
 // J~ of every step of the shallow model into J; with a latent warm-up, steps 0..T_w take P_1

@@ -157,12 +157,12 @@ __global__ __launch_bounds__(64) void k_resjac_plrnn(const float *__restrict__ A
 //   (with the k-permutation kappa(4j+q, g) = 16j + 4g + q the 16x16x4 output layout is
 //   exactly the B layout of the next step, so no data moves between steps).
 // ---------------------------------------------------------------------------------------
-template <int MP, bool REV>
+template <int MP, bool REV, bool WU>
 __global__ __launch_bounds__(64) void k_chunk_product_plrnn(
     const float *__restrict__ A, const float *__restrict__ W, float alpha, int N, const uint32_t *__restrict__ masks,
     const float *__restrict__ rhs, const float *__restrict__ z, const float *__restrict__ x, float seed_scale,
     float *__restrict__ Pout, float *__restrict__ vout, const int *__restrict__ active, int B, int T, int M, int C,
-    int ncs) {
+    int ncs, int tw) {
     using G = Geo<MP>;
     constexpr int NCH = G::NCH, NI = G::NI, NS = G::NS, MW = G::MW;
     __shared__ __align__(16) float lds[64];
@@ -208,6 +208,12 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn(
             const int row = 16 * I + 4 * g + r;
             dI[I][r] = row < M ? A[row] * p_of(row, N, alpha) : 0.f;
         }
+    // latent warm-up steps (P_1): the observed latents' rows of the diagonal term are dropped
+    float dIw[NI][4];
+#pragma unroll
+    for (int I = 0; I < NI; ++I)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dIw[I][r] = (WU && 16 * I + 4 * g + r < N) ? 0.f : dI[I][r];
     // accumulators start at the identity of each chain
     v4f acc[NI][4];
 #pragma unroll
@@ -256,10 +262,18 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn(
 #pragma unroll
                     for (int q = 0; q < 4; ++q) Bop[4 * j + q] = select_bit(wj, 16 * (j & 1) + 4 * g + q, acc[j][Jt][q]);
                 }
+                const bool warm = WU && plo[n] + t <= tw;   // J~ of step plo + t with P_1
+                if (warm) {
+#pragma unroll
+                    for (int j = 0; j < NS / 4; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            if (16 * j + 4 * g + q < N) Bop[4 * j + q] = 0.f;
+                }
 #pragma unroll
                 for (int I = 0; I < NI; ++I)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) acc[I][Jt][r] *= dI[I][r];
+                    for (int r = 0; r < 4; ++r) acc[I][Jt][r] *= warm ? dIw[I][r] : dI[I][r];
 #pragma unroll
                 for (int I = 0; I < NI; ++I)
 #pragma unroll
@@ -271,11 +285,12 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn(
         if (!REV) {
             const int s = ulo + t;
             const size_t step = (size_t)ub * T + s;
+            const float uo = (WU && ui < N && s <= tw) ? 0.f : u;   // P_s u
             float w = 0.f;
-            if (run && ui < M) w = mask_bit(masks, step, MW, ui) ? u : 0.f;
+            if (run && ui < M) w = mask_bit(masks, step, MW, ui) ? uo : 0.f;
             lds[lane] = w;
             lds_barrier();
-            const float y = fmaf(du, u, lds_dot<MP>(lds, un, wv));
+            const float y = fmaf(du, uo, lds_dot<MP>(lds, un, wv));
             lds_barrier();
             if (run && ui < M) u = y - rhs[step * M + ui];
         } else {
@@ -287,13 +302,15 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn(
             if (run && ui < M) {
                 const size_t step = (size_t)ub * T + k;
                 float y = 0.f;
-                if (t > 0) {
+                if (t > 0 && !(WU && ui < N && k + 1 <= tw)) {   // P_{k+1} = P_1 drops observed rows
                     const float m = (float)mask_bit(masks, step + 1, MW, ui);
                     y = pu * fmaf(Au, u, m * wt);
                 }
                 float gk;
                 if (rhs) gk = rhs[step * M + ui];
-                else gk = ui < N ? seed_scale * (z[step * M + ui] - x[((size_t)ub * (T + 1) + k + 1) * N + ui]) : 0.f;
+                else gk = (ui < N && (!WU || k >= tw))
+                              ? seed_scale * (z[step * M + ui] - x[((size_t)ub * (T + 1) + k + 1) * N + ui])
+                              : 0.f;
                 u = y + gk;
             }
         }
@@ -325,20 +342,20 @@ __global__ __launch_bounds__(64) void k_chunk_product_plrnn(
 // r_t = z_t - F, and advances both the chunk product and the chunk-local solution.
 // r and the masks are written for the fix-up pass.  Same MFMA layout as above.
 // ---------------------------------------------------------------------------------------
-template <int MP>
+template <int MP, bool WU>
 __global__ __launch_bounds__(64) void k_newton_product_plrnn(
     const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
     const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
     const int *__restrict__ zsel, float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout,
     float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
-    int ncs) {
+    int ncs, int tw) {
     using G = Geo<MP>;
     constexpr int NCH = G::NCH, NI = G::NI, NS = G::NS, MW = G::MW;
     __shared__ __align__(16) float lds[64];
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int nchains = B * ncs;
     const int chain0 = blockIdx.x * NCH;
-    int plen[NCH];
+    int plen[NCH], cst[NCH];              // steps and first step of each chain
     float gam[NCH];                       // damping of the linearisation (1 = exact Newton)
     int maxlen = 0;
 #pragma unroll
@@ -349,6 +366,7 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
         ok = ok && (!active || active[b]);
         const int s0 = cc * C;
         plen[n] = ok ? min(C, T - s0) : 0;
+        cst[n] = s0;
         gam[n] = gamma ? gamma[b] : 1.f;
         maxlen = max(maxlen, plen[n]);
     }
@@ -379,6 +397,12 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
             for (int r = 0; r < 4; ++r) dI[I][r] *= gam[0];
         }
     }
+    // latent warm-up steps (P_1): the observed latents' rows of the diagonal term are dropped
+    float dIw[NI][4];
+#pragma unroll
+    for (int I = 0; I < NI; ++I)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dIw[I][r] = (WU && 16 * I + 4 * g + r < N) ? 0.f : dI[I][r];
     v4f acc[NI][4];
 #pragma unroll
     for (int Jt = 0; Jt < 4; ++Jt) {
@@ -444,7 +468,7 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
         float zt = 0.f;
         if (run) {
             if (s == 0 || !forced) zt = zprev;
-            else zt = __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xb));
+            else zt = forced_in<WU>(pi, alpha, zprev, xb, s, tw);
         }
         const bool pos = zt > 0.f;
         const uint64_t bal = __ballot(pos);
@@ -482,6 +506,14 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
 #pragma unroll
                     for (int q = 0; q < 4; ++q) Bop[4 * j + q] = select_bit(wj, 16 * (j & 1) + 4 * g + q, acc[j][Jt][q]);
                 }
+                const bool warm = WU && cst[n] + t <= tw;   // P_1: the observed latents' rows dropped
+                if (warm) {
+#pragma unroll
+                    for (int j = 0; j < NS / 4; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            if (16 * j + 4 * g + q < N) Bop[4 * j + q] = 0.f;
+                }
                 if (NCH > 1 && gam[n] != 1.f) {   // damped chain (uniform branch)
                     const float gm = gam[n];
 #pragma unroll
@@ -494,7 +526,7 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
 #pragma unroll
                 for (int I = 0; I < NI; ++I)
 #pragma unroll
-                    for (int r2 = 0; r2 < 4; ++r2) acc[I][Jt][r2] *= dI[I][r2];
+                    for (int r2 = 0; r2 < 4; ++r2) acc[I][Jt][r2] *= warm ? dIw[I][r2] : dI[I][r2];
 #pragma unroll
                 for (int I = 0; I < NI; ++I)
 #pragma unroll
@@ -502,9 +534,10 @@ __global__ __launch_bounds__(64) void k_newton_product_plrnn(
             }
         }
         // chunk-local solution: u <- gamma (d u + W (p m u)) - r
-        lds[lane] = pos ? pi * u : 0.f;
+        const float uo = (WU && forced && us0 + t <= tw) ? 0.f : u;   // P_s u
+        lds[lane] = pos ? pi * uo : 0.f;
         lds_barrier();
-        const float y = fmaf(di, u, lds_dot<MP>(lds, un, wrow));
+        const float y = fmaf(di, uo, lds_dot<MP>(lds, un, wrow));
         lds_barrier();
         if (run) {
             u = fmaf(ugam, y, -r);
@@ -1989,12 +2022,13 @@ __device__ __forceinline__ float lds_row_dot64(const float (*wl)[68], int row, c
 // and the chunk-local solution are row dot products against the same LDS rows, corrected for
 // the diagonal: F_i = (W + diag A)_i relu(z~) + A_i min(z~_i, 0), and
 // y_i = (W + diag A)_i (m o u) + A_i u_i (1 - m_i).
+template <bool WU>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_newton_product_plrnn64u(
     const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
     const float *__restrict__ x, const float *__restrict__ z0, const float *zbuf, const float *zalt,
     const int *__restrict__ zsel, float *__restrict__ r_out, uint32_t *__restrict__ masks, float *__restrict__ Pout,
     float *__restrict__ vout, const int *__restrict__ active, const float *__restrict__ gamma, int B, int T, int M, int C,
-    int ncs) {
+    int ncs, int tw) {
     constexpr int MP = 64, NI = 4;
     __shared__ __align__(16) float wl[MP][68];   // W + diag(A), zero padded
     __shared__ __align__(16) float lds[64];
@@ -2011,6 +2045,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_
     const float p = N > 0 ? __fsub_rn(1.0f, alpha) : 1.0f;
     const float gp = (gamma ? gamma[b] : 1.f) * p;
     const float gp2 = gp * gp, gp4 = gp2 * gp2, gp8 = gp4 * gp4;
+    // latent warm-up with every latent observed (N = M): the Jacobians of steps s <= tw are zero
+    // (P_1 = 0), so a chunk that holds one has P = 0 (the product runs unchanged and is zeroed at
+    // the end) and u restarts from -r there; N = 0 has no observed latent and no change
+    const bool warmchunk = WU && N > 0 && s0 <= tw;
     // diagonal entries of this lane's A fragments: row 16 I + c is column 16 I + 4 g + q where
     // c == 4 g + q; there the masked entry is A instead of 0
     uint32_t dgA[NI][4];
@@ -2089,7 +2127,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_
         float zt = 0.f;
         if (run) {
             if (s == 0 || !forced) zt = zprev;
-            else zt = __fadd_rn(__fmul_rn(p, zprev), __fmul_rn(alpha, xb));
+            else zt = forced_in<WU>(p, alpha, zprev, xb, s, tw);
         }
         const bool pos = zt > 0.f;
         const uint64_t bal = __ballot(pos);
@@ -2122,7 +2160,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_
         const float y = fmaf(Ai, pos ? 0.f : u, lds_row_dot64(wl, ui, lds));
         lds_barrier();
         if (run) {
-            u = fmaf(gp, y, -r);
+            const float gps = (warmchunk && s <= tw) ? 0.f : gp;   // J~_s = 0 in a warm-up step
+            u = fmaf(gps, y, -r);
             zprev = zcur;
         }
     };
@@ -2139,7 +2178,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_
             for (int I = 0; I < NI; ++I) acc[I][Jt] = acc2[I][Jt];
     }
     if (ok0 && len > 0) {
-        float rest = 1.f;
+        float rest = warmchunk ? 0.f : 1.f;
         for (int k = 0; k < (len & 7); ++k) rest *= gp;
         float *P = Pout + (size_t)id * MP * MP;
 #pragma unroll
@@ -2987,14 +3026,14 @@ __global__ __launch_bounds__(WALK_NWV * 64) void k_carry_walk16(const float *__r
 // ---------------------------------------------------------------------------------------
 // forward fix-up: Delta from the carry, z += Delta, per-sequence max |Delta|
 // ---------------------------------------------------------------------------------------
-template <int MP>
+template <int MP, bool WU>
 __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict__ A, const float *__restrict__ W,
                                                         float alpha, int N, const uint32_t *__restrict__ masks,
                                                         const float *__restrict__ r, const float *__restrict__ carry_in,
                                                         float *zbuf, float *zalt, const int *__restrict__ zsel,
                                                         uint32_t *__restrict__ chain_bits, const int *__restrict__ active,
                                                         const float *__restrict__ gamma, int B, int T, int M, int C,
-                                                        int ncs) {
+                                                        int ncs, int tw) {
     using G = Geo<MP>;
     __shared__ __align__(16) float lds[64];
     const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
@@ -3038,9 +3077,10 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict_
             mq[q] = mq[q + 1];
         }
         fetch(t + PD, rq[PD - 1], zq[PD - 1], mq[PD - 1]);
-        lds[lane] = (run && ((mc >> (i & 31)) & 1u)) ? D : 0.f;
+        const float Do = (WU && i < N && s0 + t <= tw) ? 0.f : D;   // P_1 in a latent warm-up step
+        lds[lane] = (run && ((mc >> (i & 31)) & 1u)) ? Do : 0.f;
         lds_barrier();
-        const float y = fmaf(d, D, lds_dot<MP>(lds, n, wrow));
+        const float y = fmaf(d, Do, lds_dot<MP>(lds, n, wrow));
         lds_barrier();
         if (run) {
             D = fmaf(gm, y, -rc);
@@ -3074,7 +3114,7 @@ __global__ __launch_bounds__(64) void k_fixup_fwd_plrnn(const float *__restrict_
 // The same update as k_fixup_fwd_plrnn, 16 MFMAs per wave and step instead of an M-long dot
 // product per lane.
 // ---------------------------------------------------------------------------------------
-template <int MP, bool VEC>
+template <int MP, bool VEC, bool WU>
 __global__ __launch_bounds__(MP * 4) void k_fixup_fwd_plrnn_mf(const float *__restrict__ A, const float *__restrict__ W,
                                                                float alpha, int N, const uint32_t *__restrict__ masks,
                                                                const float *__restrict__ r,
@@ -3083,7 +3123,7 @@ __global__ __launch_bounds__(MP * 4) void k_fixup_fwd_plrnn_mf(const float *__re
                                                                uint32_t *__restrict__ chain_bits,
                                                                const int *__restrict__ active,
                                                                const float *__restrict__ gamma, int B, int T, int M,
-                                                               int C, int ncs) {
+                                                               int C, int ncs, int tw) {
     using G = Geo<MP>;
     constexpr int NW = MP / 16, NS = MP / 4, DQ = MP + 4;
     __shared__ __align__(16) float dls[2][16 * DQ];   // [buffer][chain c][latent]
@@ -3191,6 +3231,17 @@ __global__ __launch_bounds__(MP * 4) void k_fixup_fwd_plrnn_mf(const float *__re
                 bv[4 * j + 1] = select_bit(w, sh + 1, dq.y);
                 bv[4 * j + 2] = select_bit(w, sh + 2, dq.z);
                 bv[4 * j + 3] = select_bit(w, sh + 3, dq.w);
+            }
+            if constexpr (WU) {   // a latent warm-up step of chain c (P_1): observed entries of Delta dropped
+                if (s0 + t <= tw) {
+#pragma unroll
+                    for (int k = 0; k < NS; ++k)
+                        if (16 * (k / 4) + 4 * g + (k % 4) < N) bv[k] = 0.f;
+                    own.x = i0 < N ? 0.f : own.x;
+                    own.y = i0 + 1 < N ? 0.f : own.y;
+                    own.z = i0 + 2 < N ? 0.f : own.z;
+                    own.w = i0 + 3 < N ? 0.f : own.w;
+                }
             }
             // two accumulators over alternate k-steps: half the dependent chain
             v4f acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
@@ -3366,14 +3417,14 @@ int launch_ctl_init(const NewtonDev &nd, uint32_t *seq, int B, hipStream_t st) {
 // sums of this chunk: dW[i][j] += lam_i relu(z~_j), dA_i += lam_i z~_i, dh_i += lam_i
 // (layout gpart[chain][MP][MP + 2]).
 // ---------------------------------------------------------------------------------------
-template <int MP>
+template <int MP, bool WU>
 __global__ __launch_bounds__(64) void k_fixup_rev_plrnn(const float *__restrict__ A, const float *__restrict__ W,
                                                         float alpha, int N, const uint32_t *__restrict__ masks,
                                                         const float *__restrict__ gin, float seed_scale,
                                                         const float *__restrict__ x, const float *__restrict__ z0,
                                                         const float *__restrict__ z, const float *__restrict__ carry_in,
                                                         float *__restrict__ lam_out, float *__restrict__ gpart, int B,
-                                                        int T, int M, int C, int ncs) {
+                                                        int T, int M, int C, int ncs, int tw) {
     using G = Geo<MP>;
     __shared__ __align__(16) float lds[64];
     const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
@@ -3402,8 +3453,9 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn(const float *__restrict_
             const size_t step = (size_t)b * T + k;
             if (k + 1 < T) mv = (float)mask_bit(masks, step + 1, G::MW, i);
             if (gin) gv = gin[step * M + i];
-            else if (i < N) gv = seed_scale * (z[step * M + i] - x[((size_t)b * (T + 1) + k + 1) * N + i]);
-            zv = forced_state(x, z0, z, b, k, i, T, M, N, alpha);
+            else if (i < N && (!WU || k >= tw))   // no MSE seed for the warm-up states
+                gv = seed_scale * (z[step * M + i] - x[((size_t)b * (T + 1) + k + 1) * N + i]);
+            zv = forced_state(x, z0, z, b, k, i, T, M, N, alpha, WU ? tw : 0);
         }
     };
     constexpr int PD = 1;
@@ -3428,7 +3480,9 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn(const float *__restrict_
         float zt = 0.f;
         if (run) {
             const size_t step = (size_t)b * T + k;
-            const float y = (k + 1 < T) ? pi * fmaf(Ai, lam, mc * wt) : 0.f;
+            // J~_{k+1}^T lam, P_{k+1} = P_1 dropping the observed rows in a latent warm-up step
+            const bool jon = k + 1 < T && !(WU && i < N && k + 1 <= tw);
+            const float y = jon ? pi * fmaf(Ai, lam, mc * wt) : 0.f;
             lam = y + gk;
             if (lam_out) lam_out[step * M + i] = lam;
             zt = zc;
@@ -3598,16 +3652,18 @@ int launch_chunk_product_plrnn(const PlrnnArgs &a, bool rev, const uint32_t *mas
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
-    if (a.tw > 0) return invalid_arg("the stored-mask chunk product takes no latent warm-up");
     KTimer kt("k_chunk_product_plrnn", st);
-#define CP(MPV, R)                                                                                                  \
-    hipLaunchKernelGGL((k_chunk_product_plrnn<MPV, R>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, \
-                       rhs, z, a.x, seed_scale, P, v, active, a.B, a.T, a.M, C, ncs)
+#define CP(MPV, R, WUV)                                                                                              \
+    hipLaunchKernelGGL((k_chunk_product_plrnn<MPV, R, WUV>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N,    \
+                       masks, rhs, z, a.x, seed_scale, P, v, active, a.B, a.T, a.M, C, ncs, a.tw)
+#define CPW(MPV, R) \
+    if (a.tw > 0) CP(MPV, R, true); else CP(MPV, R, false);
     if (!rev) {
-        if (MP == 16) CP(16, false); else if (MP == 32) CP(32, false); else CP(64, false);
+        if (MP == 16) { CPW(16, false) } else if (MP == 32) { CPW(32, false) } else { CPW(64, false) }
     } else {
-        if (MP == 16) CP(16, true); else if (MP == 32) CP(32, true); else CP(64, true);
+        if (MP == 16) { CPW(16, true) } else if (MP == 32) { CPW(32, true) } else { CPW(64, true) }
     }
+#undef CPW
 #undef CP
     DEER_LAUNCH_CHECK("k_chunk_product_plrnn");
     return DEER_OK;
@@ -3622,16 +3678,23 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
     KTimer kt("k_newton_product_plrnn", st);
     if (wmaps == 2 && (MP != 16 || ncs % 32 || !gmap))
         return invalid_arg("group maps need M <= 16, a chunk count divisible by 32 and their buffer");
-#define NP(MPV)                                                                                                   \
-    hipLaunchKernelGGL(k_newton_product_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, \
-                       a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs)
+#define NP(MPV)                                                                                                    \
+    if (a.tw > 0)                                                                                                  \
+        hipLaunchKernelGGL((k_newton_product_plrnn<MPV, true>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, \
+                           a.N, a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs, a.tw); \
+    else                                                                                                           \
+        hipLaunchKernelGGL((k_newton_product_plrnn<MPV, false>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, \
+                           a.N, a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs, 0)
     if (wmaps && (MP != 16 || ncs % 4))
         return invalid_arg("composed wave maps need M <= 16 and a chunk count divisible by 4");
     if (mark && MP != 16) return invalid_arg("pass marks are written by the M <= 16 forward pass only");
-    if (a.tw > 0 && MP != 16) return invalid_arg("the latent warm-up inside the Newton iteration needs M <= 16");
     if (MP == 64 && (a.N == 0 || a.N == a.M)) {   // uniform forcing factor: W-in-LDS kernel
-        hipLaunchKernelGGL(k_newton_product_plrnn64u, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0,
-                           z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs);
+        if (a.tw > 0)
+            hipLaunchKernelGGL(k_newton_product_plrnn64u<true>, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N,
+                               a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs, a.tw);
+        else
+            hipLaunchKernelGGL(k_newton_product_plrnn64u<false>, dim3(nch), dim3(64), 0, st, a.A, a.W, a.h, a.alpha,
+                               a.N, a.x, a.z0, z, zalt, zsel, r, masks, P, v, active, gamma, a.B, a.T, a.M, C, ncs, 0);
     } else if (MP == 16) {
 #define NP16(TBV, WPBV)                                                                                                \
     hipLaunchKernelGGL((k_newton_product_plrnn16<TBV, WPBV, WUV>), dim3(grid / WPBV), dim3(64 * WPBV), 0, st, a.A, a.W, \
@@ -3652,7 +3715,11 @@ int launch_newton_product_plrnn(const PlrnnArgs &a, const float *z, const float 
         }
 #undef NP16W
 #undef NP16
-    } else if (MP == 32) NP(32); else NP(64);
+    } else if (MP == 32) {
+        NP(32);
+    } else {
+        NP(64);
+    }
 #undef NP
     DEER_LAUNCH_CHECK("k_newton_product_plrnn");
     return DEER_OK;
@@ -3778,9 +3845,13 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
     KTimer kt("k_fixup_fwd_plrnn", st);
-#define FX(MPV)                                                                                                       \
-    hipLaunchKernelGGL(k_fixup_fwd_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, carry_in, \
-                       z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
+#define FX(MPV)                                                                                                        \
+    if (a.tw > 0)                                                                                                      \
+        hipLaunchKernelGGL((k_fixup_fwd_plrnn<MPV, true>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, r, \
+                           carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs, a.tw);        \
+    else                                                                                                               \
+        hipLaunchKernelGGL((k_fixup_fwd_plrnn<MPV, false>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, \
+                           r, carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs, 0)
 #define FX16(TBV)                                                                                                 \
     hipLaunchKernelGGL((k_fixup_fwd_plrnn16<TBV, WUV>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x,  \
                        a.z0, carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs, Pm, vm, gmap, \
@@ -3789,7 +3860,6 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     if (Pm && (MP != 16 || ncs % 4))
         return invalid_arg("composed wave maps need M <= 16 and a chunk count divisible by 4");
     if (fc && MP != 16) return invalid_arg("the fused pass-end control needs M <= 16");
-    if (a.tw > 0 && MP != 16) return invalid_arg("the latent warm-up inside the Newton iteration needs M <= 16");
     FusedCtl fcv{};
     if (fc) fcv = *fc;
     if (MP == 16) {
@@ -3802,17 +3872,27 @@ int launch_fixup_fwd_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
         }
     } else if (fixup_mfma()) {
         const int gridm = (nch + 15) / 16;
-#define FXM(MPV, VV)                                                                                                 \
-    hipLaunchKernelGGL((k_fixup_fwd_plrnn_mf<MPV, VV>), dim3(gridm), dim3(MPV * 4), 0, st, a.A, a.W, a.alpha, a.N, masks, \
-                       r, carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs)
+#define FXM(MPV, VV)                                                                                                  \
+    if (a.tw > 0)                                                                                                     \
+        hipLaunchKernelGGL((k_fixup_fwd_plrnn_mf<MPV, VV, true>), dim3(gridm), dim3(MPV * 4), 0, st, a.A, a.W, a.alpha, \
+                           a.N, masks, r, carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, C, ncs,  \
+                           a.tw);                                                                                     \
+    else                                                                                                              \
+        hipLaunchKernelGGL((k_fixup_fwd_plrnn_mf<MPV, VV, false>), dim3(gridm), dim3(MPV * 4), 0, st, a.A, a.W,       \
+                           a.alpha, a.N, masks, r, carry_in, z, zalt, zsel, chain_bits, active, gamma, a.B, a.T, a.M, \
+                           C, ncs, 0)
         const bool v4 = (a.M & 3) == 0;
         if (MP == 32) {
-            if (v4) FXM(32, true); else FXM(32, false);
+            if (v4) { FXM(32, true); } else { FXM(32, false); }
         } else {
-            if (v4) FXM(64, true); else FXM(64, false);
+            if (v4) { FXM(64, true); } else { FXM(64, false); }
         }
 #undef FXM
-    } else if (MP == 32) FX(32); else FX(64);
+    } else if (MP == 32) {
+        FX(32);
+    } else {
+        FX(64);
+    }
 #undef FX16
 #undef FX
     DEER_LAUNCH_CHECK("k_fixup_fwd_plrnn");
@@ -3824,12 +3904,21 @@ int launch_fixup_rev_plrnn(const PlrnnArgs &a, const uint32_t *masks, const floa
     const int MP = padded(a.M);
     const int nch = a.B * ncs;
     const int grid = (nch + (64 / MP) - 1) / (64 / MP);
-    if (a.tw > 0) return invalid_arg("the stored-mask reverse fix-up takes no latent warm-up");
     KTimer kt("k_fixup_rev_plrnn", st);
-#define FR(MPV)                                                                                                     \
-    hipLaunchKernelGGL(k_fixup_rev_plrnn<MPV>, dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, g,       \
-                       seed_scale, a.x, a.z0, z, carry_in, lam, gpart, a.B, a.T, a.M, C, ncs)
-    if (MP == 16) FR(16); else if (MP == 32) FR(32); else FR(64);
+#define FR(MPV)                                                                                                      \
+    if (a.tw > 0)                                                                                                    \
+        hipLaunchKernelGGL((k_fixup_rev_plrnn<MPV, true>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N, masks, \
+                           g, seed_scale, a.x, a.z0, z, carry_in, lam, gpart, a.B, a.T, a.M, C, ncs, a.tw);         \
+    else                                                                                                             \
+        hipLaunchKernelGGL((k_fixup_rev_plrnn<MPV, false>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.alpha, a.N,     \
+                           masks, g, seed_scale, a.x, a.z0, z, carry_in, lam, gpart, a.B, a.T, a.M, C, ncs, 0)
+    if (MP == 16) {
+        FR(16);
+    } else if (MP == 32) {
+        FR(32);
+    } else {
+        FR(64);
+    }
 #undef FR
     DEER_LAUNCH_CHECK("k_fixup_rev_plrnn");
     return DEER_OK;

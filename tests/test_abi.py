@@ -105,18 +105,19 @@ def test_warmup_arguments(lib):
     st = lib.deer_solve(ctypes.byref(m), ctypes.byref(bad), ctypes.byref(o), 2, 64, None, None, None, None,
                         None, None, None, 0, None)
     assert st == _b.DEER_ERR_INVALID_ARG and b"T_w" in lib.deer_last_error()
-    # M <= 16: the warm-up is part of the one Newton iteration, which needs no more workspace
-    for op in (_b.DEER_OP_SOLVE, _b.DEER_OP_ADJOINT):
-        assert lib.deer_workspace_bytes_ex(ctypes.byref(m), ctypes.byref(fw), 2, 64, op, 0) == \
-            lib.deer_workspace_bytes(ctypes.byref(m), 2, 64, op)
-    # M > 16 chains two solves (the warm-up prefix, then the rest), which need a tolerance
+    # GTF-DEER: the warm-up is part of the one Newton iteration, which needs no more workspace
     m20, _keep20 = _vanilla_model(20)
-    assert lib.deer_workspace_bytes_ex(ctypes.byref(m20), ctypes.byref(fw), 2, 64, _b.DEER_OP_SOLVE, 0) > 0
+    ms, _keeps = _vanilla_model(16, _b.DEER_SHPLRNN)
+    for mm in (m, m20, ms):
+        for op in (_b.DEER_OP_SOLVE, _b.DEER_OP_ADJOINT):
+            assert lib.deer_workspace_bytes_ex(ctypes.byref(mm), ctypes.byref(fw), 2, 64, op, 0) == \
+                lib.deer_workspace_bytes(ctypes.byref(mm), 2, 64, op)
+    # quasi-DEER chains two solves (the warm-up prefix, then the rest), which need a tolerance
     fixed = _b.deer_solve_opts(1e-5, 10, 3, 0, 0.0)
     dummy = (ctypes.c_float * 16)()
     p = ctypes.cast(dummy, ctypes.c_void_p)
-    st = lib.deer_solve(ctypes.byref(m20), ctypes.byref(fw), ctypes.byref(fixed), 2, 64, p, None, p, None,
-                        None, None, None, 0, None)
+    st = lib.deer_solve_quasi(ctypes.byref(m20), ctypes.byref(fw), ctypes.byref(fixed), 2, 64, p, None, p, None,
+                              None, None, None, 0, None)
     assert st == _b.DEER_ERR_INVALID_ARG and b"tolerance" in lib.deer_last_error()
     dg = _b.deer_model(_b.DEER_DIAG_SSM, 4, 3, m.A, m.W, None, None, None)
     assert lib.deer_workspace_bytes_ex(ctypes.byref(dg), ctypes.byref(fw), 2, 64, _b.DEER_OP_SOLVE, 0) == 0

@@ -48,11 +48,11 @@ def test_update_rows_counts_each_update_over_its_part():
 
 
 def test_warmup_in_one_iteration_where_the_library_takes_it():
-    # vanilla PLRNN M <= 16 (GTF-DEER): one iteration, every update over all T steps
+    # GTF-DEER: one iteration, every update over all T steps
     assert bench.warmup_in_one_iteration("plrnn", 16, False)
     assert bench.warmup_in_one_iteration("plrnn", 3, False)
-    # chained solves elsewhere
-    assert not bench.warmup_in_one_iteration("plrnn", 17, False)
+    assert bench.warmup_in_one_iteration("plrnn", 64, False)
+    # quasi-DEER chains two solves
     assert not bench.warmup_in_one_iteration("plrnn", 16, True)
     assert bench.warmup_in_one_iteration("shplrnn", 64, False)
     assert not bench.warmup_in_one_iteration("shplrnn", 16, True)

@@ -20,7 +20,7 @@ if not torch.cuda.is_available():
 import paper_2605_12683_amd as D  # noqa: E402
 
 TOL = 1e-4
-_ENV = ("DEER_CHUNK", "DEER_GROUP_MAPS", "DEER_PASS_FUSION", "DEER_SH_FUSED", "DEER_SH_RESMFMA")
+_ENV = ("DEER_CHUNK", "DEER_GROUP_MAPS", "DEER_PASS_FUSION", "DEER_FIX_MFMA", "DEER_SH_FUSED", "DEER_SH_RESMFMA")
 
 
 @pytest.fixture(autouse=True)
@@ -82,14 +82,17 @@ def test_warmup_with_given_cotangent_and_initial_state():
         assert rel_inf(v.cpu().numpy(), gr[k]) < TOL, k
 
 
-# M <= 16: the warm-up is part of the one Newton iteration (the register-tiled kernels take the
-# forcing strength per step: alpha_s = 1 and P_1 for s <= T_w).  T_w at the first step, inside a
+# Vanilla PLRNN: the warm-up is part of the one Newton iteration (the kernels take the forcing
+# strength per step: alpha_s = 1 and P_1 for s <= T_w).  M <= 16: T_w at the first step, inside a
 # chunk and a tile, on a chunk boundary (T_w + 1 divisible by the chunk length) and next to the
 # end; chunk layouts through the per-step slow paths (ragged tiles), composed wave maps, group
-# maps and the fused pass kernel; every latent observed; M = 3 (the one-launch kernels step aside).
+# maps and the fused pass kernel; every latent observed; M = 3 (the one-launch kernels step
+# aside).  M > 16: 32- and 64-wide kernels, M not a multiple of 4, ragged chunks, every latent
+# observed (the uniform-forcing M = 64 kernel steps aside).
 JOINT = [(16, 3, 2, 700, 100, 0), (16, 3, 2, 2048, 511, 16), (16, 3, 2, 2048, 700, 16), (12, 4, 2, 4096, 1, 32),
          (12, 4, 2, 4096, 4094, 32), (7, 3, 3, 640, 77, 40), (5, 2, 3, 1000, 333, 25), (16, 16, 2, 513, 200, 0),
-         (3, 3, 1, 300, 17, 0)]
+         (3, 3, 1, 300, 17, 0), (24, 24, 3, 1000, 999, 0), (33, 5, 2, 700, 333, 37), (40, 10, 2, 300, 1, 0),
+         (64, 64, 2, 513, 200, 0), (61, 7, 2, 400, 150, 64)]
 
 
 def _joint_case(M, N, B, T, T_w, chunk, seed):
@@ -120,15 +123,16 @@ def test_warmup_one_iteration_newton_iterates(M, N, B, T, T_w, chunk):
 @pytest.mark.parametrize("M,N,B,T,T_w,chunk", JOINT)
 def test_warmup_one_iteration_counts_and_adjoint(M, N, B, T, T_w, chunk):
     """Solved to tolerance the joint iteration reaches the warm-up rollout in the oracle's number
-    of updates (up to one), with the fused pass kernel and with separate kernels; the adjoint
-    and gradients (MSE over the states after the warm-up, and a given cotangent) match the
-    oracle's joint recursion."""
+    of updates (up to one), with the fused pass kernel and with separate kernels (M <= 16), with
+    the matrix-core and the lane-per-latent fix-up (M > 16); the adjoint and gradients (MSE over
+    the states after the warm-up, and a given cotangent) match the oracle's joint recursion."""
     c = _joint_case(M, N, B, T, T_w, chunk, 4200 + M + T_w)
     m = oracle_model(c)
     ref = O.rollout(m, c.x, c.alpha, N, T_w=T_w)
     want = O.newton(m, c.x, c.alpha, N, tol=1e-5, T_w=T_w)["iters"].tolist()
     for fuse in ("1", "0"):
         os.environ["DEER_PASS_FUSION"] = fuse
+        os.environ["DEER_FIX_MFMA"] = fuse
         say("warm-up one iteration to tolerance", M, N, B, T, T_w, chunk, fuse)
         res = D.deer_solve(m, c.x, c.alpha, N, tol=1e-5, max_iter=200, T_w=T_w)
         assert res["status"] == 0, res

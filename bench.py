@@ -11,9 +11,8 @@ One step = one pass of the whole path over one batch of synthetic input:
                    read-out gradients), then deer_adjoint on that real cotangent (reverse scan
                    with conj(lambda) + dlambda / dBc reductions).
 Inputs are resident in HBM before the timed region.  The value is DEER timesteps per
-second: sum over sequences of T x Newton updates, per second of the whole step (with a latent
-warm-up, --tw, where the library chains a solve of steps 1..T_w and one of the rest, an update
-is counted at the length of the part it covered: T_w or T - T_w).
+second: sum over sequences of T x Newton updates, per second of the whole step (a latent
+warm-up, --tw, is part of the same Newton iteration, so every update spans the T steps).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 5]
 
@@ -59,24 +58,6 @@ def _plrnn_step(D, model, xd, c, ws_s, ws_a, T_w=0):
     return sum(res["iters"])
 
 
-def warmup_in_one_iteration(kind, M, quasi):
-    """The library runs the latent warm-up inside the one Newton iteration for GTF-DEER on both
-    PLRNN kinds (identity read-out); quasi-DEER chains two solves."""
-    return not quasi and kind in ("plrnn", "shplrnn")
-
-
-def update_rows(T, T_w, updates, warm_updates, nsteps):
-    """(b, t) steps covered by `updates` Newton updates (summed over sequences and `nsteps`
-    steps).  Without a warm-up every update spans T steps; with one, `warm_updates` per step
-    belong to the warm-up part (T_w steps each) and the rest to steps T_w + 1..T."""
-    if warm_updates is None:
-        return updates * T
-    rest = updates - warm_updates * nsteps
-    if rest < 0:
-        raise ValueError("fewer updates than the warm-up part alone takes")
-    return T_w * warm_updates * nsteps + (T - T_w) * rest
-
-
 def check_quasi_bound(c, passes):
     """Refuse, before any GPU work, a quasi-DEER solve to tolerance whose pass bound (T + 2:
     about one more exact leading step per update) is too long for a benchmark run; a fixed
@@ -88,14 +69,14 @@ def check_quasi_bound(c, passes):
                          f"(> {QUASI_MAX_PASSES}); pass --quasi-passes K to time K passes per solve instead")
 
 
-def _quasi_step(D, model, xd, c, ws_s, ws_a):
+def _quasi_step(D, model, xd, c, ws_s, ws_a, T_w=0):
     # quasi-DEER: one more leading step is exact per update, so T + 1 updates always suffice
     # (check_quasi_bound has refused the workloads where that is too many)
     res = D.deer_solve_quasi(model, xd, c.alpha, c.n_obs, tol=c.tol, max_iter=c.T + 2, fixed_iters=c.fixed_iters,
-                             ws=ws_s, check=False)
+                             ws=ws_s, check=False, T_w=T_w)
     if res["status"] != 0:
         raise RuntimeError(f"deer_solve_quasi returned status {res['status']}: {D.load().deer_last_error()}")
-    D.deer_adjoint_quasi(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a, want_lam=False)
+    D.deer_adjoint_quasi(model, xd, res["z"], c.alpha, c.n_obs, ws=ws_a, want_lam=False, T_w=T_w)
     return sum(res["iters"])
 
 
@@ -116,14 +97,13 @@ def _diag_step(D, model, readout, xd, c, ws_s, ws_r, ws_a, bufs):
     return c.B
 
 
-def kernel_work(c, steps, updates, fwd_rows=None):
+def kernel_work(c, steps, updates):
     """Algorithmic work of each kernel over the timed region: {name: (bound, total work)};
-    work in flop (mfma) or bytes (hbm).  `updates` = Newton updates summed over sequences;
-    `fwd_rows` (latent warm-up) = the (b, t) steps those updates covered, when an update does
-    not span the whole sequence."""
+    work in flop (mfma) or bytes (hbm).  `updates` = Newton updates summed over sequences, each
+    over the whole sequence."""
     B, T, M, N = c.B, c.T, c.M, c.n_obs
     W = (M + 31) // 32
-    fwd = updates * T if fwd_rows is None else fwd_rows   # (b, t) steps processed by the updates
+    fwd = updates * T                 # (b, t) steps processed by the updates
     adj = steps * B * T               # (b, t) steps of the adjoint passes
     prod = fwd + steps * B * (T - 1)  # chunk-product steps (the adjoint product covers 1..T-1)
     if c.kind == "diag_ssm":
@@ -245,9 +225,9 @@ def measured_mfma(workload, kernel):
             "source": f"profiles/mfma_{workload}.txt"}
 
 
-def roofline_for(name, c, total_ms, launches, steps, updates, fwd_rows=None):
+def roofline_for(name, c, total_ms, launches, steps, updates):
     """Algorithmic work of the dominant kernel over the timed region, divided by its time."""
-    work = kernel_work(c, steps, updates, fwd_rows)
+    work = kernel_work(c, steps, updates)
     base = {"kernel": name, "avg_launch_ms": total_ms / launches, "launches": launches,
             "traffic": measured_traffic(c.name, name)}
     if name not in work:
@@ -499,7 +479,7 @@ def main():
             ws_s = D._workspace(lib.deer_quasi_workspace_bytes(ctypes.byref(model.c), c.B, c.T, Bnd.DEER_OP_SOLVE))
             ws_a = D._workspace(lib.deer_quasi_workspace_bytes(ctypes.byref(model.c), c.B, c.T,
                                                                Bnd.DEER_OP_ADJOINT))
-            step = lambda: _quasi_step(D, model, xd, c, ws_s, ws_a)        # noqa: E731
+            step = lambda: _quasi_step(D, model, xd, c, ws_s, ws_a, args.tw)   # noqa: E731
         else:
             lib = D.load()
             fw = Bnd.deer_forcing(float(c.alpha), int(c.n_obs), int(args.tw))
@@ -511,21 +491,6 @@ def main():
     else:
         print(f"workload {c.name}: model kind {c.kind} not supported by this build", file=sys.stderr)
         sys.exit(3)
-
-    # latent warm-up: inside the one Newton iteration every update covers all T steps; where the
-    # library solves steps 1..T_w (alpha = 1) and then the rest, an update of the first part
-    # covers T_w steps and one of the rest T - T_w.  The first part's update count is that of the
-    # same solve run on its own (deterministic), taken once, untimed.
-    warm_updates = None
-    if (args.tw and c.kind in ("plrnn", "shplrnn") and not args.quasi
-            and not warmup_in_one_iteration(c.kind, c.M, args.quasi)):
-        r1 = D.deer_solve(model, xd[:, :args.tw + 1].contiguous(), 1.0, c.n_obs, tol=c.tol, max_iter=c.max_iter,
-                          check=False)
-        warm_updates = int(sum(r1["iters"]))
-        log(f"[bench] latent warm-up part: {warm_updates} updates over {args.tw} steps (summed over sequences)")
-
-    def rows_of(upd, nsteps):
-        return update_rows(c.T, args.tw, upd, warm_updates, nsteps)
 
     t_w = time.perf_counter()
     for i in range(args.warmup):
@@ -559,7 +524,7 @@ def main():
     log(f"[bench] {args.steps} timed steps: {(t1 - t0) * 1e3 / args.steps:.3f} ms per step")
     dt = t1 - t0
     iters_per_step = updates / args.steps
-    timesteps = rows_of(updates, args.steps)
+    timesteps = updates * c.T
     value = timesteps / dt
     for k, (ms, n) in sorted(kt.items(), key=lambda kv: -kv[1][0]):
         log(f"[bench] {k:28s} {ms:10.3f} ms total  {n:6d} launches  {ms / n:9.4f} ms avg")
@@ -567,10 +532,9 @@ def main():
     # work model (a latency-bound helper such as the carry pass has none)
     modeled = {k: v for k, v in kt.items() if k in kernel_work(c, 1, 1)}
     dom = max((modeled or kt).items(), key=lambda kv: kv[1][0])
-    prof_rows = rows_of(prof_updates, prof_steps)
-    roof = roofline_for(dom[0], c, dom[1][0], dom[1][1], prof_steps, prof_updates, prof_rows)
+    roof = roofline_for(dom[0], c, dom[1][0], dom[1][1], prof_steps, prof_updates)
     kernels = {k: {"ms_total": ms, "launches": n, **({"frac": r["frac"], "unit": r["unit"], "achieved": r["achieved"]}
-                                                      if (r := roofline_for(k, c, ms, n, prof_steps, prof_updates, prof_rows))["frac"]
+                                                      if (r := roofline_for(k, c, ms, n, prof_steps, prof_updates))["frac"]
                                                       is not None else {})}
                for k, (ms, n) in kt.items()}
 
@@ -592,8 +556,7 @@ def main():
                    "fixed_iters": c.fixed_iters or None, "newton_updates_per_step": iters_per_step,
                    "step": ("deer_train_step (solve, MSE + MAR loss, gradient, Adam)" if args.train else
                             "deer_solve_quasi + deer_adjoint_quasi (quasi-DEER: diagonal Jacobians)" if args.quasi
-                            else "deer_solve + deer_adjoint"), "latent_warmup": args.tw,
-                   "warmup_part_updates_per_step": warm_updates},
+                            else "deer_solve + deer_adjoint"), "latent_warmup": args.tw},
         "roofline": roof,
         "kernels": kernels,
     }

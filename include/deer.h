@@ -99,9 +99,7 @@ typedef struct {
     int T_w;            /* latent warm-up (Alg. GTF-DEER, latent state warm-up paragraph):
                            0 <= T_w < T; the forced inputs z~_1..z~_{T_w} use alpha = 1 and
                            the MSE seed leaves z_1..z_{T_w} out (1 / (N (T - T_w))).  PLRNN
-                           kinds; the workspace is deer_workspace_bytes_ex(...).  Quasi-DEER
-                           chains two problems (see there) and needs a tolerance
-                           (fixed_iters = 0).                                               */
+                           kinds; the workspace is deer_workspace_bytes_ex(...).            */
     const float *obs;   /* general observation matrix B [n_forced, M] (device, row-major) of the
                            read-out x^_t = B z_t, or NULL for the identity read-out B = [I_N 0].
                            With B given (PLRNN kinds, 1 <= n_forced <= 64, n_forced may exceed
@@ -151,16 +149,11 @@ enum { DEER_SCAN_DENSE = 0, DEER_SCAN_DIAG_C64 = 1 };
 size_t deer_workspace_bytes(const deer_model *model, int B, int T, int op);
 
 /* The same for any forcing, warm-up included, and for the quasi-DEER entry points when
- * quasi != 0.  With T_w > 0 and GTF-DEER (both PLRNN kinds) the warm-up is part of the one
- * Newton iteration (Alg. GTF-DEER: the kernels take alpha_s = 1 and P_1 for s <= T_w), so iters
- * and fixed_iters count updates of the whole sequence and the workspace is
- * deer_workspace_bytes's.  Quasi-DEER runs it as two chained solves -- the warm-up prefix with
- * alpha = 1, then the rest from z_0 := P_1 z_{T_w} + zbar_{T_w} -- which have the joint
- * problem's unique zero (the segments are copied through the workspace), and the adjoint as
- * the rest's adjoint followed by the prefix's, seeded with diag(J~_{T_w+1}) lam_{T_w+1}; the
- * parameter gradients are summed.  The two solves share opts->max_iter: the rest runs at most
- * the passes the warm-up part left (at least one), so iters reports the updates of both.  With
- * an observation matrix (forcing->obs) the warm-up is part of the one Newton iteration too. */
+ * quasi != 0.  A latent warm-up (T_w > 0) is part of the one Newton iteration (Alg. GTF-DEER:
+ * the kernels take alpha_s = 1 and P_1 for s <= T_w; quasi-DEER the same in its diagonal
+ * coefficients), so iters and fixed_iters count updates of the whole sequence and, with the
+ * identity read-out, the workspace is that of the plain solve.  With an observation matrix
+ * (forcing->obs) the workspace holds the projectors and the stored Jacobians. */
 size_t deer_workspace_bytes_ex(const deer_model *model, const deer_forcing *forcing, int B, int T, int op,
                                int quasi);
 

@@ -144,93 +144,6 @@ __global__ void k_copy_sel(float *__restrict__ z, const float *__restrict__ zalt
         for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < seq_elems; e += stride) d[e] = s[e];
     }
 }
-// rows [src_off, src_off + rows) of every sequence of a [B, src_rows, width] array of 32-bit
-// words into rows [dst_off, ...) of a [B, dst_rows, width] array (one sequence per grid row)
-__global__ void k_copy_rows(uint32_t *__restrict__ dst, const uint32_t *__restrict__ src, int rows, int width,
-                            int src_rows, int src_off, int dst_rows, int dst_off) {
-    const int b = blockIdx.y;
-    const size_t n = (size_t)rows * width;
-    const uint32_t *sp = src + ((size_t)b * src_rows + src_off) * width;
-    uint32_t *dp = dst + ((size_t)b * dst_rows + dst_off) * width;
-    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n; e += (size_t)gridDim.x * blockDim.x)
-        dp[e] = sp[e];
-}
-static int copy_rows(void *dst, const void *src, int B, int rows, int width, int src_rows, int src_off, int dst_rows,
-                     int dst_off, hipStream_t st) {
-    const size_t n = (size_t)rows * width;
-    if (n == 0 || B == 0) return DEER_OK;
-    const size_t want = (n + 255) / 256;
-    const int gx = (int)(want < 1024 ? want : 1024);
-    hipLaunchKernelGGL(k_copy_rows, dim3(gx, B), dim3(256), 0, st, (uint32_t *)dst, (const uint32_t *)src, rows, width,
-                       src_rows, src_off, dst_rows, dst_off);
-    DEER_LAUNCH_CHECK("k_copy_rows");
-    return DEER_OK;
-}
-
-// initial state of the part after the warm-up: P_1 z_{T_w} + zbar_{T_w} = [x_{T_w}; z_{T_w}[N:]]
-__global__ void k_warmup_state(const float *__restrict__ x, const float *__restrict__ z1, float *__restrict__ zb, int T,
-                               int T1, int M, int N) {
-    const int b = blockIdx.x;
-    for (int i = threadIdx.x; i < M; i += blockDim.x)
-        zb[(size_t)b * M + i] = i < N ? x[((size_t)b * (T + 1) + T1) * N + i] : z1[((size_t)b * T1 + T1 - 1) * M + i];
-}
-
-// cotangent the warm-up prefix receives from the rest: g1[b, T1 - 1] += J~_{T_w+1}^T lam2[b, 0],
-// J~_{T_w+1} = J_F(zb) P_1 (diag(J_F(zb)) P_1 for quasi-DEER); P_1 zeroes the observed latents.
-// The hidden ReLU decision of the shallow model is taken as everywhere else (u accumulated from
-// h2 left to right, a rounding after every multiply and add).
-__global__ void k_warmup_cotangent(int kind, int quasi, const float *__restrict__ A, const float *__restrict__ W,
-                                   const float *__restrict__ W2, const float *__restrict__ h2, int M, int L, int N,
-                                   const float *__restrict__ zb, const float *__restrict__ lam2, int T2,
-                                   float *__restrict__ g1, int T1) {
-    extern __shared__ float sh[];   // lam [M], zb [M], shallow: per hidden unit [L]
-    const int b = blockIdx.x, t = threadIdx.x;
-    float *lm = sh, *zs = sh + M, *dl = sh + 2 * M;
-    for (int e = t; e < M; e += blockDim.x) {
-        lm[e] = lam2[(size_t)b * T2 * M + e];
-        zs[e] = zb[(size_t)b * M + e];
-    }
-    __syncthreads();
-    if (kind == DEER_SHPLRNN) {
-        for (int l = t; l < L; l += blockDim.x) {
-            float u = h2 ? h2[l] : 0.f;
-            for (int j = 0; j < M; ++j) u = __fadd_rn(u, __fmul_rn(W2[(size_t)l * M + j], zs[j]));
-            float a = 0.f;
-            if (!quasi)
-                for (int i = 0; i < M; ++i) a = fmaf(W[(size_t)i * L + l], lm[i], a);
-            dl[l] = u > 0.f ? (quasi ? 1.f : a) : 0.f;
-        }
-        __syncthreads();
-    }
-    for (int j = t; j < M; j += blockDim.x) {
-        float v;
-        if (kind == DEER_PLRNN) {
-            const bool m = zs[j] > 0.f;
-            if (quasi) {
-                v = (A[j] + (m ? W[(size_t)j * M + j] : 0.f)) * lm[j];
-            } else {
-                float a = 0.f;
-                for (int i = 0; i < M; ++i) a = fmaf(W[(size_t)i * M + j], lm[i], a);
-                v = A[j] * lm[j] + (m ? a : 0.f);
-            }
-        } else if (quasi) {
-            float d = 0.f;
-            for (int l = 0; l < L; ++l)
-                if (dl[l] != 0.f) d += W[(size_t)j * L + l] * W2[(size_t)l * M + j];
-            v = (A[j] + d) * lm[j];
-        } else {
-            float a = 0.f;
-            for (int l = 0; l < L; ++l) a = fmaf(W2[(size_t)l * M + j], dl[l], a);
-            v = A[j] * lm[j] + a;
-        }
-        if (j >= N) g1[((size_t)b * T1 + T1 - 1) * M + j] += v;
-    }
-}
-
-__global__ void k_add_f32(float *__restrict__ out, const float *__restrict__ a, const float *__restrict__ b, size_t n) {
-    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n; e += (size_t)gridDim.x * blockDim.x)
-        out[e] = a[e] + b[e];
-}
 
 __global__ void k_fill_f32(float *p, size_t n, float v) {
     for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n; e += (size_t)gridDim.x * blockDim.x) p[e] = v;
@@ -862,13 +775,6 @@ static int init_guess(const deer_solve_opts *o, int B, int T, int M, int N, cons
     return DEER_OK;
 }
 
-// The latent warm-up inside the one Newton iteration (per-step forcing strength in the kernels):
-// GTF-DEER with the identity read-out, both PLRNN kinds.  Quasi-DEER solves the warm-up prefix
-// and the rest as two chained problems (solve_warmup below).
-static bool warmup_joint(const deer_model *m, const deer_forcing *f) {
-    return f->T_w > 0 && !f->obs && (m->kind == DEER_PLRNN || m->kind == DEER_SHPLRNN);
-}
-
 // J~ of every step of the shallow model into J; with a latent warm-up, steps 0..T_w take P_1
 // (alpha = 1; step 0's Jacobian only multiplies the fixed initial state's zero update) and the
 // rest P_alpha
@@ -1219,6 +1125,7 @@ static int solve_quasi(const deer_model *m, const deer_forcing *f, const deer_so
     QuasiWs w = carve_quasi(ws, B, T, m->M, L, DEER_OP_SOLVE, &need);
     PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
     ShArgs sa{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
+    a.tw = sa.tw = f->T_w;
     if ((rc = init_guess(o, B, T, m->M, f->n_forced, x, z, st))) return rc;
     std::vector<int> act(B, 1), it(B, 0);
     std::vector<float> norm(B, NAN);
@@ -1244,18 +1151,6 @@ static int solve_quasi(const deer_model *m, const deer_forcing *f, const deer_so
     return finish_solve(o, B, it, norm, nonfinite, act, iters, final_norm);
 }
 
-// ---- latent warm-up as two chained problems ---------------------------------------------
-// The warm-up prefix (steps 1..T_w, forced inputs with alpha = 1) does not depend on the rest,
-// and the rest starts from the fully forced z~_{T_w} = P_1 z_{T_w} + zbar_{T_w}; the chained
-// solves therefore have the joint problem's unique zero.  Segments are copied through the
-// workspace (sequences of different lengths do not share the batch stride).
-struct WarmWs {
-    float *x1, *x2, *z1, *z2, *zb, *g1, *g2, *lam1, *lam2, *gr1, *gr2;
-    uint32_t *m1, *m2;
-    void *inner;
-    size_t inner_bytes;
-};
-
 static size_t param_floats(const deer_model *m) {
     return m->kind == DEER_PLRNN ? (size_t)m->M * (m->M + 2) : (size_t)m->M * (2 * m->L + 2) + m->L;
 }
@@ -1276,157 +1171,6 @@ static deer_grads grads_at(const deer_model *m, float *base) {
     return g;
 }
 
-static WarmWs carve_warm(void *ws, const deer_model *m, const deer_forcing *f, int B, int T, int op, bool quasi,
-                         size_t *bytes) {
-    WarmWs w{};
-    const int T1 = f->T_w, T2 = T - f->T_w, N = f->n_forced, M = m->M;
-    const int H = m->kind == DEER_PLRNN ? M : m->L;
-    const size_t W = (H + 31) / 32;
-    Carver c(ws);
-    w.x1 = c.take<float>((size_t)B * (T1 + 1) * N);
-    w.x2 = c.take<float>((size_t)B * (T2 + 1) * N);
-    w.z1 = c.take<float>((size_t)B * T1 * M);
-    w.z2 = c.take<float>((size_t)B * T2 * M);
-    w.zb = c.take<float>((size_t)B * M);
-    if (op == DEER_OP_SOLVE) {
-        w.m1 = c.take<uint32_t>((size_t)B * T1 * W);
-        w.m2 = c.take<uint32_t>((size_t)B * T2 * W);
-    } else {
-        w.g1 = c.take<float>((size_t)B * T1 * M);
-        w.g2 = c.take<float>((size_t)B * T2 * M);
-        w.lam1 = c.take<float>((size_t)B * T1 * M);
-        w.lam2 = c.take<float>((size_t)B * T2 * M);
-        w.gr1 = c.take<float>(param_floats(m));
-        w.gr2 = c.take<float>(param_floats(m));
-    }
-    const size_t i1 = quasi ? deer_quasi_workspace_bytes(m, B, T1, op) : deer_workspace_bytes(m, B, T1, op);
-    const size_t i2 = quasi ? deer_quasi_workspace_bytes(m, B, T2, op) : deer_workspace_bytes(m, B, T2, op);
-    w.inner_bytes = i1 > i2 ? i1 : i2;
-    w.inner = c.take<char>(w.inner_bytes);
-    *bytes = c.off;
-    return w;
-}
-
-static int solve_warmup(const deer_model *m, const deer_forcing *f, const deer_solve_opts *o, int B, int T,
-                        const float *x, const float *z0, float *z, uint32_t *masks, int32_t *iters, float *final_norm,
-                        void *ws, size_t ws_bytes, hipStream_t st, bool quasi) {
-    if (o->fixed_iters > 0) {
-        set_error("the latent warm-up runs with a tolerance (fixed_iters = 0)");
-        return DEER_ERR_INVALID_ARG;
-    }
-    size_t need = 0;
-    carve_warm(nullptr, m, f, B, T, DEER_OP_SOLVE, quasi, &need);
-    int rc = check_ws(ws, ws_bytes, need);
-    if (rc) return rc;
-    WarmWs w = carve_warm(ws, m, f, B, T, DEER_OP_SOLVE, quasi, &need);
-    const int T1 = f->T_w, T2 = T - f->T_w, N = f->n_forced, M = m->M;
-    const int W = ((m->kind == DEER_PLRNN ? M : m->L) + 31) / 32;
-    if ((rc = copy_rows(w.x1, x, B, T1 + 1, N, T + 1, 0, T1 + 1, 0, st))) return rc;
-    if ((rc = copy_rows(w.x2, x, B, T2 + 1, N, T + 1, T1, T2 + 1, 0, st))) return rc;
-    if (o->init == DEER_INIT_USER) {
-        if ((rc = copy_rows(w.z1, z, B, T1, M, T, 0, T1, 0, st))) return rc;
-        if ((rc = copy_rows(w.z2, z, B, T2, M, T, T1, T2, 0, st))) return rc;
-    }
-    const deer_forcing f1{1.0f, N, 0}, f2{f->alpha, N, 0};
-    std::vector<int32_t> it1(B, 0), it2(B, 0);
-    std::vector<float> n1(B, 0.f), n2(B, 0.f);
-    auto solve = quasi ? deer_solve_quasi : deer_solve;
-    const int r1 = solve(m, &f1, o, B, T1, w.x1, z0, w.z1, masks ? w.m1 : nullptr, it1.data(), n1.data(), w.inner,
-                         w.inner_bytes, st);
-    if (r1 != DEER_OK && r1 != DEER_ERR_NOT_CONVERGED && r1 != DEER_ERR_NONFINITE) return r1;
-    hipLaunchKernelGGL(k_warmup_state, dim3(B), dim3(64), 0, st, x, (const float *)w.z1, w.zb, T, T1, M, N);
-    DEER_LAUNCH_CHECK("k_warmup_state");
-    // the two parts share the pass budget: the rest gets what the warm-up part left (at least one
-    // pass); a pass is an accepted or rejected update, so the warm-up part took at least max it1
-    deer_solve_opts o2 = *o;
-    {
-        const int cap = o->max_iter > 0 ? o->max_iter : 500;
-        int used = 0;
-        for (int b = 0; b < B; ++b) used = it1[b] > used ? it1[b] : used;
-        o2.max_iter = cap - used > 1 ? cap - used : 1;
-    }
-    const int r2 = solve(m, &f2, &o2, B, T2, w.x2, w.zb, w.z2, masks ? w.m2 : nullptr, it2.data(), n2.data(), w.inner,
-                         w.inner_bytes, st);
-    if (r2 != DEER_OK && r2 != DEER_ERR_NOT_CONVERGED && r2 != DEER_ERR_NONFINITE) return r2;
-    if ((rc = copy_rows(z, w.z1, B, T1, M, T1, 0, T, 0, st))) return rc;
-    if ((rc = copy_rows(z, w.z2, B, T2, M, T2, 0, T, T1, st))) return rc;
-    if (masks) {
-        if ((rc = copy_rows(masks, w.m1, B, T1, W, T1, 0, T, 0, st))) return rc;
-        if ((rc = copy_rows(masks, w.m2, B, T2, W, T2, 0, T, T1, st))) return rc;
-    }
-    for (int b = 0; b < B; ++b) {
-        if (iters) iters[b] = it1[b] + it2[b];
-        if (final_norm) final_norm[b] = n1[b] > n2[b] || isnan(n1[b]) ? n1[b] : n2[b];
-    }
-    if (r1 != DEER_OK || r2 != DEER_OK) {
-        set_error("latent warm-up: the warm-up part returned %d, the rest %d", r1, r2);
-        return r1 == DEER_ERR_NONFINITE || r2 == DEER_ERR_NONFINITE ? DEER_ERR_NONFINITE : DEER_ERR_NOT_CONVERGED;
-    }
-    return DEER_OK;
-}
-
-static int adjoint_warmup(const deer_model *m, const deer_forcing *f, int B, int T, const float *x, const float *z0,
-                          const float *z, const float *g, float *lam, const deer_grads *grads, void *ws,
-                          size_t ws_bytes, hipStream_t st, bool quasi) {
-    size_t need = 0;
-    carve_warm(nullptr, m, f, B, T, DEER_OP_ADJOINT, quasi, &need);
-    int rc = check_ws(ws, ws_bytes, need);
-    if (rc) return rc;
-    WarmWs w = carve_warm(ws, m, f, B, T, DEER_OP_ADJOINT, quasi, &need);
-    const int T1 = f->T_w, T2 = T - f->T_w, N = f->n_forced, M = m->M;
-    if ((rc = copy_rows(w.x1, x, B, T1 + 1, N, T + 1, 0, T1 + 1, 0, st))) return rc;
-    if ((rc = copy_rows(w.x2, x, B, T2 + 1, N, T + 1, T1, T2 + 1, 0, st))) return rc;
-    if ((rc = copy_rows(w.z1, z, B, T1, M, T, 0, T1, 0, st))) return rc;
-    if ((rc = copy_rows(w.z2, z, B, T2, M, T, T1, T2, 0, st))) return rc;
-    hipLaunchKernelGGL(k_warmup_state, dim3(B), dim3(64), 0, st, x, (const float *)w.z1, w.zb, T, T1, M, N);
-    DEER_LAUNCH_CHECK("k_warmup_state");
-    const bool want_grads = grads && (grads->A || grads->W || grads->W2 || grads->h || grads->h2);
-    const deer_grads gr1 = grads_at(m, w.gr1), gr2 = grads_at(m, w.gr2);
-    const deer_forcing f1{1.0f, N, 0}, f2{f->alpha, N, 0};
-    // the rest: its own MSE seed (normalised by its T - T_w steps) or the given cotangent
-    if (g && (rc = copy_rows(w.g2, g, B, T2, M, T, T1, T2, 0, st))) return rc;
-    rc = quasi ? deer_adjoint_quasi(m, &f2, B, T2, w.x2, w.zb, w.z2, g ? w.g2 : nullptr, w.lam2,
-                                    want_grads ? &gr2 : nullptr, w.inner, w.inner_bytes, st)
-               : deer_adjoint(m, &f2, B, T2, w.x2, w.zb, w.z2, g ? w.g2 : nullptr, w.lam2, want_grads ? &gr2 : nullptr,
-                              w.inner, w.inner_bytes, st);
-    if (rc) return rc;
-    // the prefix: no loss of its own (or the given cotangent), plus what the rest hands back
-    if (g) {
-        if ((rc = copy_rows(w.g1, g, B, T1, M, T, 0, T1, 0, st))) return rc;
-    } else if ((rc = launch_fill_f32(w.g1, (size_t)B * T1 * M, 0.f, st))) {
-        return rc;
-    }
-    const size_t shb = (size_t)(2 * M + (m->kind == DEER_SHPLRNN ? m->L : 0)) * sizeof(float);
-    hipLaunchKernelGGL(k_warmup_cotangent, dim3(B), dim3(64), shb, st, m->kind, quasi ? 1 : 0, m->A, m->W, m->W2, m->h2,
-                       M, m->L, N, (const float *)w.zb, (const float *)w.lam2, T2, w.g1, T1);
-    DEER_LAUNCH_CHECK("k_warmup_cotangent");
-    rc = quasi ? deer_adjoint_quasi(m, &f1, B, T1, w.x1, z0, w.z1, w.g1, w.lam1, want_grads ? &gr1 : nullptr, w.inner,
-                                    w.inner_bytes, st)
-               : deer_adjoint(m, &f1, B, T1, w.x1, z0, w.z1, w.g1, w.lam1, want_grads ? &gr1 : nullptr, w.inner,
-                              w.inner_bytes, st);
-    if (rc) return rc;
-    if (lam) {
-        if ((rc = copy_rows(lam, w.lam1, B, T1, M, T1, 0, T, 0, st))) return rc;
-        if ((rc = copy_rows(lam, w.lam2, B, T2, M, T2, 0, T, T1, st))) return rc;
-    }
-    if (want_grads) {
-        const size_t M_ = M, L_ = m->L;
-        struct Part { float *out; const float *a, *b; size_t n; };
-        const bool sh = m->kind == DEER_SHPLRNN;
-        const Part parts[5] = {{grads->A, gr1.A, gr2.A, M_},
-                               {grads->W, gr1.W, gr2.W, sh ? M_ * L_ : M_ * M_},
-                               {sh ? grads->W2 : nullptr, gr1.W2, gr2.W2, L_ * M_},
-                               {grads->h, gr1.h, gr2.h, M_},
-                               {sh ? grads->h2 : nullptr, gr1.h2, gr2.h2, L_}};
-        for (const Part &pt : parts) {
-            if (!pt.out) continue;
-            hipLaunchKernelGGL(k_add_f32, dim3((unsigned)((pt.n + 255) / 256)), dim3(256), 0, st, pt.out, pt.a, pt.b,
-                               pt.n);
-            DEER_LAUNCH_CHECK("k_add_f32");
-        }
-    }
-    return DEER_OK;
-}
 
 }  // namespace deer
 
@@ -1586,8 +1330,6 @@ int deer_solve(const deer_model *m, const deer_forcing *f, const deer_solve_opts
     if (m->kind != DEER_DIAG_SSM && o->fixed_iters <= 0 && (rc = check_host_reserved(B))) return rc;
     hipStream_t st = (hipStream_t)stream;
     if (f->obs) return solve_obs(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
-    if (f->T_w > 0 && !warmup_joint(m, f))
-        return solve_warmup(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st, false);
     if (m->kind == DEER_PLRNN)
         return solve_plrnn(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, st);
     if (m->kind == DEER_SHPLRNN)
@@ -1631,7 +1373,6 @@ int deer_adjoint_ex(const deer_model *m, const deer_forcing *f, int B, int T, co
         set_error("the latent warm-up takes the native cotangent layout");
         return DEER_ERR_INVALID_ARG;
     }
-    if (f->T_w > 0 && !warmup_joint(m, f)) return adjoint_warmup(m, f, B, T, x, z0, z, g, lam, grads, ws, ws_bytes, st, false);
     if (m->kind == DEER_PLRNN) {
         size_t need = 0;
         carve_plrnn(nullptr, B, T, m->M, DEER_OP_ADJOINT, &need);
@@ -1731,8 +1472,6 @@ int deer_solve_quasi(const deer_model *m, const deer_forcing *f, const deer_solv
     if (o->init < 0 || o->init > 2) { set_error("unknown init %d", o->init); return DEER_ERR_INVALID_ARG; }
     if (!(o->tol >= 0.f) && o->fixed_iters <= 0) { set_error("tol must be >= 0"); return DEER_ERR_INVALID_ARG; }
     if (o->fixed_iters <= 0 && (rc = check_host_reserved(B))) return rc;
-    if (f->T_w > 0)
-        return solve_warmup(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, (hipStream_t)stream, true);
     return solve_quasi(m, f, o, B, T, x, z0, z, masks, iters, final_norm, ws, ws_bytes, (hipStream_t)stream);
 }
 
@@ -1744,18 +1483,20 @@ int deer_adjoint_quasi(const deer_model *m, const deer_forcing *f, int B, int T,
     if (rc) return rc;
     if (!x || !z) { set_error("x and z are required"); return DEER_ERR_INVALID_ARG; }
     hipStream_t st = (hipStream_t)stream;
-    if (f->T_w > 0) return adjoint_warmup(m, f, B, T, x, z0, z, g, lam, grads, ws, ws_bytes, st, true);
     size_t need = 0;
     const int L = quasi_L(m);
     carve_quasi(nullptr, B, T, m->M, L, DEER_OP_ADJOINT, &need);
     if ((rc = check_ws(ws, ws_bytes, need))) return rc;
     QuasiWs w = carve_quasi(ws, B, T, m->M, L, DEER_OP_ADJOINT, &need);
     PlrnnArgs a{m->A, m->W, m->h, f->alpha, f->n_forced, x, z0, B, T, m->M};
-    const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * T)) : 0.f;
+    a.tw = f->T_w;
+    // MSE over the states after the latent warm-up, z_{T_w+1}..z_T
+    const float scale = f->n_forced > 0 ? (float)(2.0 / ((double)B * f->n_forced * (T - f->T_w))) : 0.f;
     if (L > 0) {
         // shallow: masks and coefficients at z, the reverse scan writes lam, then the shallow
         // gradient kernel (dA, dW1, dW2, dh1, dh2) from it
         ShArgs sa{m->A, m->W, m->W2, m->h, m->h2, f->alpha, f->n_forced, x, z0, B, T, m->M, m->L};
+        sa.tw = f->T_w;
         float *lo = lam ? lam : w.lam;
         if ((rc = launch_resjac_shplrnn(sa, z, nullptr, nullptr, nullptr, nullptr, w.masks, nullptr, st))) return rc;
         if ((rc = launch_qdeer_shdiag(sa, w.masks, nullptr, nullptr, w.coef, st))) return rc;
@@ -1780,14 +1521,9 @@ size_t deer_workspace_bytes_ex(const deer_model *m, const deer_forcing *f, int B
         carve_obs(nullptr, m, f, B, T, op, &bytes);
         return bytes;
     }
-    if (!f || f->T_w == 0) return quasi ? deer_quasi_workspace_bytes(m, B, T, op) : deer_workspace_bytes(m, B, T, op);
-    if ((quasi ? check_quasi(m, f, B, T) : check_common(m, f, B, T)) != DEER_OK) return 0;
-    if (!quasi && warmup_joint(m, f) && (op == DEER_OP_SOLVE || op == DEER_OP_ADJOINT))
-        return deer_workspace_bytes(m, B, T, op);   // one iteration over the whole sequence
-    if (op != DEER_OP_SOLVE && op != DEER_OP_ADJOINT) return 0;
-    size_t bytes = 0;
-    carve_warm(nullptr, m, f, B, T, op, quasi != 0, &bytes);
-    return bytes;
+    // a latent warm-up is part of the one Newton iteration: the workspace of the plain solve
+    if (f && f->T_w > 0 && (quasi ? check_quasi(m, f, B, T) : check_common(m, f, B, T)) != DEER_OK) return 0;
+    return quasi ? deer_quasi_workspace_bytes(m, B, T, op) : deer_workspace_bytes(m, B, T, op);
 }
 
 size_t deer_train_params(const deer_model *m) {

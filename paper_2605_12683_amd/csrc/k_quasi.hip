@@ -65,7 +65,7 @@ __global__ __launch_bounds__(64) void k_qdeer_resdiag(const float *__restrict__ 
                                                       const float *zbuf, const float *zalt, const int *__restrict__ zsel,
                                                       const int *__restrict__ active, const float *__restrict__ gamma,
                                                       float *__restrict__ rhs, float *__restrict__ coef, int B, int T,
-                                                      int M) {
+                                                      int M, int tw) {
     constexpr int NCH = 64 / MP;
     constexpr int NG = 4;             // row groups per iteration (memory parallelism)
     constexpr int RS = NCH * NG;      // steps per iteration
@@ -109,7 +109,10 @@ __global__ __launch_bounds__(64) void k_qdeer_resdiag(const float *__restrict__ 
 #pragma unroll
         for (int q = 0; q < NG; ++q) {
             const int s = sb + q * NCH + n;
-            zt[q] = s == 0 ? zinit : (forced ? __fadd_rn(__fmul_rn(pi, zp[q]), __fmul_rn(alpha, xq[q])) : zp[q]);
+            // latent warm-up (s <= tw): the observed latents take the data (alpha_s = 1)
+            zt[q] = s == 0 ? zinit
+                           : (forced ? (s <= tw ? xq[q] : __fadd_rn(__fmul_rn(pi, zp[q]), __fmul_rn(alpha, xq[q])))
+                                     : zp[q]);
             zc[q] = zv[q];
         }
         load(sb + stride);   // the next iteration's inputs, in flight during this one
@@ -129,7 +132,7 @@ __global__ __launch_bounds__(64) void k_qdeer_resdiag(const float *__restrict__ 
         for (int q = 0; q < NG; ++q) {
             const int s = sb + q * NCH + n;
             if (s < T && iok) {
-                cs[(size_t)s * M] = q_coef(zt[q], Ai, Wii, pi, gmb);
+                cs[(size_t)s * M] = q_coef(zt[q], Ai, Wii, (forced && s <= tw) ? 0.f : pi, gmb);   // P_1
                 if (!REV) rs[(size_t)s * M] = zc[q] - F[q];
             }
         }
@@ -151,7 +154,7 @@ __global__ __launch_bounds__(64) void k_qdeer_chunk(const float *__restrict__ co
                                                     float sgn, const float *__restrict__ z, const float *__restrict__ x,
                                                     float seed_scale, int N, const int *__restrict__ active,
                                                     float *__restrict__ Pout, float *__restrict__ vout, int B, int T,
-                                                    int M, int C, int ncs) {
+                                                    int M, int C, int ncs, int tw) {
     constexpr int NCH = 64 / MP;
     const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
     const int id = blockIdx.x * NCH + n;
@@ -172,9 +175,9 @@ __global__ __launch_bounds__(64) void k_qdeer_chunk(const float *__restrict__ co
             if (rhs) {
                 gv[k] = rhs[(base + s) * M + i];
             } else {
-                gv[k] = i < N ? __fmul_rn(seed_scale, __fsub_rn(z[(base + s) * M + i],
-                                                                 x[((size_t)b * (T + 1) + s + 1) * N + i]))
-                              : 0.f;
+                gv[k] = (i < N && s >= tw) ? __fmul_rn(seed_scale, __fsub_rn(z[(base + s) * M + i],
+                                                                                x[((size_t)b * (T + 1) + s + 1) * N + i]))
+                                           : 0.f;   // no MSE seed for the warm-up states s < tw
             }
         }
 #pragma unroll
@@ -327,7 +330,7 @@ __global__ __launch_bounds__(64) void k_qdeer_fixup_rev(const float *__restrict_
                                                         const float *__restrict__ x, const float *__restrict__ z0,
                                                         const float *__restrict__ z, const float *__restrict__ carry,
                                                         float *__restrict__ lam, float *__restrict__ gpart, int B,
-                                                        int T, int M, int C, int ncs) {
+                                                        int T, int M, int C, int ncs, int tw) {
     constexpr int NCH = 64 / MP;
     __shared__ __align__(16) float lds[64];
     const int lane = threadIdx.x, n = lane / MP, i = lane % MP;
@@ -356,11 +359,11 @@ __global__ __launch_bounds__(64) void k_qdeer_fixup_rev(const float *__restrict_
             if (g) {
                 gv = g[(base + s) * M + i];
             } else {
-                gv = i < N ? __fmul_rn(seed_scale, __fsub_rn(z[(base + s) * M + i],
-                                                               x[((size_t)b * (T + 1) + s + 1) * N + i]))
-                           : 0.f;
+                gv = (i < N && s >= tw) ? __fmul_rn(seed_scale, __fsub_rn(z[(base + s) * M + i],
+                                                                            x[((size_t)b * (T + 1) + s + 1) * N + i]))
+                                        : 0.f;   // no MSE seed for the warm-up states s < tw
             }
-            if (GR) zt = forced_state(x, z0, z, b, s, i, T, M, N, alpha);
+            if (GR) zt = forced_state(x, z0, z, b, s, i, T, M, N, alpha, tw);
             L = fmaf(cv, L, gv);
             if (lam) lam[(base + s) * M + i] = L;
             ga = fmaf(L, zt, ga);
@@ -401,7 +404,7 @@ __global__ __launch_bounds__(QSR) void k_qdeer_shdiag(const float *__restrict__ 
                                                      const float *__restrict__ W2, float alpha, int N,
                                                      const uint32_t *__restrict__ masks, const int *__restrict__ active,
                                                      const float *__restrict__ gamma, float *__restrict__ coef, int T,
-                                                     int M, int L) {
+                                                     int M, int L, int tw) {
     extern __shared__ float Cs[];   // [M][L]
     const int b = blockIdx.y;
     if (active && !active[b]) return;
@@ -427,7 +430,7 @@ __global__ __launch_bounds__(QSR) void k_qdeer_shdiag(const float *__restrict__ 
             for (int j = 0; j < nb; ++j)
                 if ((bits >> j) & 1u) d += cw[j];
         }
-        coef[((size_t)b * T + s) * M + i] = gm * ((Ai + d) * pi);
+        coef[((size_t)b * T + s) * M + i] = gm * ((Ai + d) * ((i < N && s <= tw) ? 0.f : pi));   // P_1 in the warm-up
     }
 }
 
@@ -439,7 +442,7 @@ int launch_qdeer_shdiag(const ShArgs &a, const uint32_t *masks, const int *activ
     if (gx > cap) gx = cap;
     KTimer kt("k_qdeer_shdiag", st);
     hipLaunchKernelGGL(k_qdeer_shdiag, dim3((unsigned)gx, (unsigned)a.B), dim3(QSR), (size_t)a.M * a.L * sizeof(float),
-                       st, a.A, a.W1, a.W2, a.alpha, a.N, masks, active, gamma, coef, a.T, a.M, a.L);
+                       st, a.A, a.W1, a.W2, a.alpha, a.N, masks, active, gamma, coef, a.T, a.M, a.L, a.tw);
     DEER_LAUNCH_CHECK("k_qdeer_shdiag");
     return DEER_OK;
 }
@@ -478,7 +481,7 @@ int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zs
         const dim3 grid = q_grid_rows(a.B, a.T, MP);
 #define RD(MPV) \
     hipLaunchKernelGGL((k_qdeer_resdiag<MPV, false>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, \
-                       (const float *)z, (const float *)zalt, zsel, active, gamma, rhs, coef, a.B, a.T, a.M)
+                       (const float *)z, (const float *)zalt, zsel, active, gamma, rhs, coef, a.B, a.T, a.M, a.tw)
         if (MP == 16) RD(16); else if (MP == 32) RD(32); else RD(64);
 #undef RD
     }
@@ -497,7 +500,7 @@ int launch_qdeer_scan_fwd(int B, int T, int M, const float *x, int N, float *z, 
         KTimer kt("k_qdeer_chunk", st);
 #define CK(MPV) \
     hipLaunchKernelGGL((k_qdeer_chunk<MPV, false>), dim3(gridc), dim3(64), 0, st, coef, rhs, -1.f, (const float *)nullptr, \
-                       x, 0.f, N, active, P, v, B, T, M, C, ncs)
+                       x, 0.f, N, active, P, v, B, T, M, C, ncs, 0)
         if (MP == 16) CK(16); else if (MP == 32) CK(32); else CK(64);
 #undef CK
     }
@@ -532,7 +535,7 @@ int launch_qdeer_adjoint(const PlrnnArgs &a, const float *g, float seed_scale, c
 #define RD(MPV) \
     hipLaunchKernelGGL((k_qdeer_resdiag<MPV, true>), dim3(grid), dim3(64), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, a.z0, z, \
                        z, (const int *)nullptr, (const int *)nullptr, (const float *)nullptr, (float *)nullptr, coef, \
-                       a.B, a.T, a.M)
+                       a.B, a.T, a.M, a.tw)
         if (MP == 16) RD(16); else if (MP == 32) RD(32); else RD(64);
 #undef RD
     }
@@ -549,7 +552,7 @@ int launch_qdeer_scan_rev(const PlrnnArgs &a, const float *g, float seed_scale, 
         KTimer kt("k_qdeer_chunk", st);
 #define CK(MPV) \
     hipLaunchKernelGGL((k_qdeer_chunk<MPV, true>), dim3(gridc), dim3(64), 0, st, coef, g, 1.f, z, a.x, \
-                       seed_scale, a.N, (const int *)nullptr, P, v, a.B, a.T, a.M, C, ncs)
+                       seed_scale, a.N, (const int *)nullptr, P, v, a.B, a.T, a.M, C, ncs, a.tw)
         if (MP == 16) CK(16); else if (MP == 32) CK(32); else CK(64);
 #undef CK
     }
@@ -567,7 +570,7 @@ int launch_qdeer_scan_rev(const PlrnnArgs &a, const float *g, float seed_scale, 
         KTimer kt("k_qdeer_fixup_rev", st);
 #define FX(MPV, GRV) \
     hipLaunchKernelGGL((k_qdeer_fixup_rev<MPV, GRV>), dim3(gridc), dim3(64), 0, st, coef, g, seed_scale, \
-                       a.alpha, a.N, a.x, a.z0, z, (const float *)carry, lam, gpart, a.B, a.T, a.M, C, ncs)
+                       a.alpha, a.N, a.x, a.z0, z, (const float *)carry, lam, gpart, a.B, a.T, a.M, C, ncs, a.tw)
 #define FXG(GRV) if (MP == 16) FX(16, GRV); else if (MP == 32) FX(32, GRV); else FX(64, GRV);
         if (gpart) { FXG(true) } else { FXG(false) }
 #undef FXG

@@ -105,20 +105,16 @@ def test_warmup_arguments(lib):
     st = lib.deer_solve(ctypes.byref(m), ctypes.byref(bad), ctypes.byref(o), 2, 64, None, None, None, None,
                         None, None, None, 0, None)
     assert st == _b.DEER_ERR_INVALID_ARG and b"T_w" in lib.deer_last_error()
-    # GTF-DEER: the warm-up is part of the one Newton iteration, which needs no more workspace
+    # the warm-up is part of the one Newton iteration (GTF-DEER and quasi-DEER, both PLRNN kinds),
+    # which needs no more workspace than the plain solve
     m20, _keep20 = _vanilla_model(20)
     ms, _keeps = _vanilla_model(16, _b.DEER_SHPLRNN)
     for mm in (m, m20, ms):
         for op in (_b.DEER_OP_SOLVE, _b.DEER_OP_ADJOINT):
             assert lib.deer_workspace_bytes_ex(ctypes.byref(mm), ctypes.byref(fw), 2, 64, op, 0) == \
                 lib.deer_workspace_bytes(ctypes.byref(mm), 2, 64, op)
-    # quasi-DEER chains two solves (the warm-up prefix, then the rest), which need a tolerance
-    fixed = _b.deer_solve_opts(1e-5, 10, 3, 0, 0.0)
-    dummy = (ctypes.c_float * 16)()
-    p = ctypes.cast(dummy, ctypes.c_void_p)
-    st = lib.deer_solve_quasi(ctypes.byref(m20), ctypes.byref(fw), ctypes.byref(fixed), 2, 64, p, None, p, None,
-                              None, None, None, 0, None)
-    assert st == _b.DEER_ERR_INVALID_ARG and b"tolerance" in lib.deer_last_error()
+            assert lib.deer_workspace_bytes_ex(ctypes.byref(mm), ctypes.byref(fw), 2, 64, op, 1) == \
+                lib.deer_quasi_workspace_bytes(ctypes.byref(mm), 2, 64, op)
     dg = _b.deer_model(_b.DEER_DIAG_SSM, 4, 3, m.A, m.W, None, None, None)
     assert lib.deer_workspace_bytes_ex(ctypes.byref(dg), ctypes.byref(fw), 2, 64, _b.DEER_OP_SOLVE, 0) == 0
 

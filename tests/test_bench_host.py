@@ -33,26 +33,3 @@ def test_host_cpu_description():
 def test_vector_peak_is_the_unpacked_fp32_rate():
     # 256 CUs x 4 SIMDs x 16 lanes x 2 flops per FMA x 2.4 GHz
     assert abs(bench.PEAK_FP32_VALU_TFLOPS - 256 * 4 * 16 * 2 * 2.4e9 / 1e12) < 0.1
-
-
-def test_update_rows_counts_each_update_over_its_part():
-    # no warm-up: every update spans the whole sequence
-    assert bench.update_rows(1000, 0, 14, None, 2) == 14 * 1000
-    # warm-up of 100 steps: per step, 3 updates of the first part (100 steps each) and the rest
-    # of 10 updates over the remaining 900 steps; over 2 steps
-    assert bench.update_rows(1000, 100, 2 * 13, 3, 2) == 2 * (3 * 100 + 10 * 900)
-    # the count never exceeds the one at the full length
-    assert bench.update_rows(1000, 100, 26, 3, 2) < 26 * 1000
-    with pytest.raises(ValueError):
-        bench.update_rows(1000, 100, 5, 3, 2)
-
-
-def test_warmup_in_one_iteration_where_the_library_takes_it():
-    # GTF-DEER: one iteration, every update over all T steps
-    assert bench.warmup_in_one_iteration("plrnn", 16, False)
-    assert bench.warmup_in_one_iteration("plrnn", 3, False)
-    assert bench.warmup_in_one_iteration("plrnn", 64, False)
-    # quasi-DEER chains two solves
-    assert not bench.warmup_in_one_iteration("plrnn", 16, True)
-    assert bench.warmup_in_one_iteration("shplrnn", 64, False)
-    assert not bench.warmup_in_one_iteration("shplrnn", 16, True)

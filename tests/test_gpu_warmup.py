@@ -197,3 +197,23 @@ def test_shallow_warmup_one_iteration(M, L, N, B, T, T_w, chunk, iterates):
     finally:
         os.environ.pop("DEER_SH_FUSED", None)
         os.environ.pop("DEER_SH_RESMFMA", None)
+
+
+@pytest.mark.parametrize("kind,M,L,N,B,T,T_w", [("plrnn", 16, 0, 3, 2, 300, 60), ("plrnn", 40, 0, 40, 2, 200, 1),
+                                                ("shplrnn", 5, 50, 3, 2, 250, 100)])
+def test_quasi_warmup_one_iteration(kind, M, L, N, B, T, T_w):
+    """Quasi-DEER takes the warm-up inside its one iteration as well (diagonal coefficients with
+    P_1 for t <= T_w): the oracle's first quasi-Newton iterates and its update counts (up to one)."""
+    c = _case(kind, M, L, N, B, T, 4400 + M + T_w)
+    m = oracle_model(c)
+    for k in (1, 2):
+        say("quasi warm-up one iteration, fixed updates", kind, M, L, N, B, T, T_w, k)
+        res = D.deer_solve_quasi(m, c.x, c.alpha, N, fixed_iters=k, T_w=T_w)
+        ref = O.newton(m, c.x, c.alpha, N, fixed_iters=k, T_w=T_w, quasi=True)
+        assert res["status"] == 0 and res["iters"] == [k] * B
+        assert rel_inf(res["z"].cpu().numpy(), ref["z"]) < TOL, k
+    say("quasi warm-up one iteration to tolerance", kind, M, L, N, B, T, T_w)
+    res = D.deer_solve_quasi(m, c.x, c.alpha, N, tol=1e-5, max_iter=T + 2, T_w=T_w)
+    want = O.newton(m, c.x, c.alpha, N, tol=1e-5, max_iter=T + 2, T_w=T_w, quasi=True)["iters"].tolist()
+    assert res["status"] == 0, res
+    assert max(abs(a - b) for a, b in zip(res["iters"], want)) <= 1, (res["iters"], want)

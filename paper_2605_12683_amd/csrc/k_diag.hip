@@ -544,22 +544,27 @@ __global__ __launch_bounds__(256) void k_diag_seg(const float *__restrict__ lam,
 // carry[s] = state at the end of segment s - 1:  X_0 = 0,  X_{s+1} = Lambda X_s + A_s,
 // Lambda = lam^seglen (conj(lam) for a reverse scan; every segment but the last is full, and
 // the last aggregate is not needed).
-// Block = (sequence, 64-channel tile), threads = (group g of CG consecutive segments, channel):
-// group aggregates, a sequential pass over the 16 groups, then every group re-walked from its
-// carry.  Serial depth 2 CG + 16 instead of nseg; the aggregates of a group are loaded
+// Block = (sequence, SEG_CT channels), threads = (group g of CG consecutive segments, channel):
+// group aggregates, a sequential pass over the SEG_NG groups, then every group re-walked from
+// its carry.  Serial depth 2 CG + SEG_NG instead of nseg; the aggregates of a group are loaded
 // SEG_CB at a time (indices clamped to the group, so the loads are unconditional) before the
 // dependent float64 updates, so the walks wait on memory once per batch rather than once per
-// segment.
-constexpr int SEG_NG = 16;
+// segment.  16 channels per block and 64 groups: 16 blocks for four sequences of 64 channels,
+// and two batches per walk for 2048 segments.
+constexpr int SEG_NG = 64;
+constexpr int SEG_CT = 16;
 constexpr int SEG_CB = 16;
 
-__global__ __launch_bounds__(1024) void k_diag_seg_carry(const float *__restrict__ lam, int conj_lam, int seglen, int B,
-                                                         int M, int nseg, int ntile, const float2 *__restrict__ agg,
-                                                         float2 *__restrict__ carry) {
-    __shared__ double ga[SEG_NG][64][2];
-    const int b = blockIdx.x / ntile, tile = blockIdx.x % ntile;
-    const int ch = threadIdx.x & 63, grp = threadIdx.x >> 6;
-    const int m = tile * 64 + ch;
+__global__ __launch_bounds__(SEG_NG * SEG_CT) void k_diag_seg_carry(const float *__restrict__ lam, int conj_lam,
+                                                                    int seglen, int B, int M, int nseg, int ntile,
+                                                                    const float2 *__restrict__ agg,
+                                                                    float2 *__restrict__ carry) {
+    __shared__ double ga[SEG_NG][SEG_CT][2];
+    constexpr int NSUB = 64 / SEG_CT;   // blocks per 64-channel tile
+    const int b = blockIdx.x / (ntile * NSUB), rem = blockIdx.x % (ntile * NSUB);
+    const int tile = rem / NSUB, sub = rem % NSUB;
+    const int ch = threadIdx.x % SEG_CT, grp = threadIdx.x / SEG_CT;
+    const int m = tile * 64 + sub * SEG_CT + ch;
     const bool mok = m < M;
     const int CG = (nseg + SEG_NG - 1) / SEG_NG;
     const int s0 = min(grp * CG, nseg), s1 = min(s0 + CG, nseg);
@@ -619,8 +624,165 @@ __global__ __launch_bounds__(1024) void k_diag_seg_carry(const float *__restrict
     }
 }
 
+// ---------------------------------------------------------------------------------------
+// Segment aggregates of the forward scan on the matrix cores (M <= 64, K <= 4 inputs).  The
+// state a full segment [t0, t0 + 512) reaches from zero is, per channel,
+//   A = sum_{a < 8} lam^{64 (7 - a)} sum_{j < K} Bc_j R_{a,j},
+//   R_{a,j} = sum_{k < 64} lam^{63 - k} u_{t0 + 64 a + k, j},
+// and R for the 64 channels (real parts in rows 0..63, imaginary parts in rows 64..127) and
+// the 32 columns (a, j) is one [128 x 64] x [64 x 32] product: A operand = the powers
+// lam^{63 - k} (LDS, formed once per block in float64), B operand = the segment's inputs
+// (LDS, transposed to [column 4 a + j][k]).  The k order is permuted as in the read-out (k-step
+// (jj, q) of lane group g is k = 16 jj + 4 g + q) so that one 16-byte LDS read gives four
+// k-steps of either operand.  The epilogue multiplies every column by lam^{64 (7 - a)} Bc_j
+// and sums the 16 columns of a tile across its lanes.  A wave takes one segment at a time; a
+// partial last segment gets an aggregate that is never used (the carries stop before it).
+// ---------------------------------------------------------------------------------------
+constexpr int AGW = 4;        // waves (segments in flight) per block
+constexpr int AQS = 68;       // LDS row stride of the powers and of the transposed inputs
+
+__global__ __launch_bounds__(AGW * 64) void k_diag_seg_agg(const float *__restrict__ lam, const float *__restrict__ Bc,
+                                                           const float *__restrict__ u, int B, int T, int M, int K,
+                                                           int nseg, float2 *__restrict__ agg) {
+    static_assert(SEG == 512, "8 blocks of 64 steps per segment");
+    __shared__ __align__(16) float qs[128][AQS];           // lam^{63-k}: re rows 0..63, im rows 64..127
+    __shared__ __align__(16) float us[AGW][32][AQS];       // inputs [4 a + j][k] of each wave's segment
+    __shared__ float2 pw[64][8], bcs[64][4];                // lam^{64 (7 - a)}, Bc_j
+    const int tid = threadIdx.x;
+    // powers in float64: a thread takes 8 consecutive k of one channel (one power, then 7 products)
+    for (int e = tid; e < 64 * 8; e += AGW * 64) {
+        const int ch = e / 8, kb = e % 8;
+        const cd l = ch < M ? cd{(double)lam[2 * ch], (double)lam[2 * ch + 1]} : cd{0.0, 0.0};
+        cd p = cpow(l, 56 - 8 * kb);   // lam^{63 - k} for k = 8 kb + 7
+        for (int k = 8 * kb + 7; k >= 8 * kb; --k) {
+            qs[ch][k] = (float)p.re;
+            qs[64 + ch][k] = (float)p.im;
+            p = cmul(p, l);
+        }
+    }
+    if (tid < 64) {
+        const int ch = tid;
+        const cd l = ch < M ? cd{(double)lam[2 * ch], (double)lam[2 * ch + 1]} : cd{0.0, 0.0};
+        const cd l64 = cpow(l, 64);
+        cd p = {1.0, 0.0};
+        for (int a = 7; a >= 0; --a) {   // lam^{64 (7 - a)}
+            pw[ch][a] = make_float2((float)p.re, (float)p.im);
+            p = cmul(p, l64);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            bcs[ch][j] = (ch < M && j < K) ? make_float2(Bc[(ch * K + j) * 2], Bc[(ch * K + j) * 2 + 1])
+                                           : make_float2(0.f, 0.f);
+    }
+    __syncthreads();
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, c = lane & 15;
+    const long total = (long)B * nseg;
+    const long stride = (long)gridDim.x * AGW;
+    // inputs of a segment: lane l holds steps t0 + 8 l .. t0 + 8 l + 7 (block a = l / 8,
+    // k = 8 (l % 8) + i), loaded a segment ahead into registers
+    float nx[8][4];
+    auto fetch = [&](long sid) {
+        const bool in = sid < total;
+        const int b = in ? (int)(sid / nseg) : 0, seg = in ? (int)(sid % nseg) : 0;
+        const int t0 = seg * SEG;
+        const int nrow = in ? min(8, T - t0 - 8 * lane) : 0;   // steps of this lane inside the sequence
+        const float *ur = u + ((long)b * (T + 1) + t0 + 8 * lane) * K;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) nx[i][j] = (i < nrow && j < K) ? ur[i * K + j] : 0.f;
+    };
+    long sid = (long)blockIdx.x * AGW + wv;
+    fetch(sid);
+    for (; sid < total; sid += stride) {
+        {
+            const int a = lane >> 3, k0 = 8 * (lane & 7);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) us[wv][4 * a + j][k0 + i] = nx[i][j];
+        }
+        wave_lds_sync();
+        fetch(sid + stride);   // in flight during this segment's products
+        v4f acc[8][2];
+#pragma unroll
+        for (int I = 0; I < 8; ++I) acc[I][0] = acc[I][1] = (v4f){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            float4 aq[8], bq[2];
+#pragma unroll
+            for (int I = 0; I < 8; ++I) aq[I] = *reinterpret_cast<const float4 *>(&qs[16 * I + c][16 * jj + 4 * g]);
+#pragma unroll
+            for (int J = 0; J < 2; ++J) bq[J] = *reinterpret_cast<const float4 *>(&us[wv][16 * J + c][16 * jj + 4 * g]);
+            // 16 independent accumulators between two products into the same one
+#pragma unroll
+            for (int J = 0; J < 2; ++J)
+#pragma unroll
+                for (int I = 0; I < 8; ++I) acc[I][J] = mfma16x16x4(aq[I].x, bq[J].x, acc[I][J]);
+#pragma unroll
+            for (int J = 0; J < 2; ++J)
+#pragma unroll
+                for (int I = 0; I < 8; ++I) acc[I][J] = mfma16x16x4(aq[I].y, bq[J].y, acc[I][J]);
+#pragma unroll
+            for (int J = 0; J < 2; ++J)
+#pragma unroll
+                for (int I = 0; I < 8; ++I) acc[I][J] = mfma16x16x4(aq[I].z, bq[J].z, acc[I][J]);
+#pragma unroll
+            for (int J = 0; J < 2; ++J)
+#pragma unroll
+                for (int I = 0; I < 8; ++I) acc[I][J] = mfma16x16x4(aq[I].w, bq[J].w, acc[I][J]);
+        }
+        // the next segment's inputs may overwrite us once every lane has read it
+        wave_lds_sync();
+        // epilogue: lane (g, c) holds rows 16 I + 4 g + r (channel 16 (I % 4) + 4 g + r, real part
+        // for I < 4, imaginary for I >= 4) of columns 16 J + c = (a = 4 J + c / 4, j = c % 4)
+        float sr[4][4], si[4][4];
+#pragma unroll
+        for (int I = 0; I < 4; ++I)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int ch = 16 * I + 4 * g + r;
+                float xr = 0.f, xi = 0.f;
+#pragma unroll
+                for (int J = 0; J < 2; ++J) {
+                    const float2 p = pw[ch][4 * J + (c >> 2)], q = bcs[ch][c & 3];
+                    const float kr = p.x * q.x - p.y * q.y, ki = p.x * q.y + p.y * q.x;   // lam^{64 (7-a)} Bc_j
+                    const float Rr = acc[I][J][r], Ri = acc[I + 4][J][r];
+                    xr = fmaf(kr, Rr, fmaf(-ki, Ri, xr));
+                    xi = fmaf(kr, Ri, fmaf(ki, Rr, xi));
+                }
+                sr[I][r] = xr;
+                si[I][r] = xi;
+            }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1)
+#pragma unroll
+            for (int I = 0; I < 4; ++I)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    sr[I][r] += __shfl_xor(sr[I][r], off, 64);
+                    si[I][r] += __shfl_xor(si[I][r], off, 64);
+                }
+        if (c == 0) {
+#pragma unroll
+            for (int I = 0; I < 4; ++I)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int ch = 16 * I + 4 * g + r;
+                    if (ch < M) agg[sid * M + ch] = make_float2(sr[I][r], si[I][r]);
+                }
+        }
+    }
+}
+
 static bool diag_seg_enabled() {
     const char *e = getenv("DEER_DIAG_SEG");
+    return !e || atoi(e) != 0;
+}
+
+// segment aggregates on the matrix cores (DEER_DIAG_AGG_MFMA=0: the lane-per-channel walk)
+static bool diag_agg_mfma() {
+    const char *e = getenv("DEER_DIAG_AGG_MFMA");
     return !e || atoi(e) != 0;
 }
 
@@ -648,14 +810,22 @@ static int launch_diag_seg(int B, int T, int M, const float *lam, const float *B
         case 3: SEGK(WR, 3, A, C, Y); break; \
         default: SEGK(WR, 4, A, C, Y); break; \
     }
-    {
+    if (M <= 64 && K <= 4 && diag_agg_mfma()) {
+        // segment aggregates on the matrix cores: a few blocks per CU, each forming the powers once
+        const long segs = (long)B * nseg;
+        const long want = (segs + AGW - 1) / AGW;
+        const int gridm = (int)(want < 512 ? want : 512);
+        KTimer _kt("k_diag_seg_reduce", st);
+        hipLaunchKernelGGL(k_diag_seg_agg, dim3(gridm), dim3(AGW * 64), 0, st, lam, Bc, u, B, T, M, K, nseg, agg);
+    } else {
         KTimer _kt("k_diag_seg_reduce", st);
         SEGALL(false, agg, (const float2 *)nullptr, (float *)nullptr)
     }
     DEER_LAUNCH_CHECK("k_diag_seg<reduce>");
     {
         KTimer _kt("k_diag_seg_carry", st);
-        hipLaunchKernelGGL(k_diag_seg_carry, dim3(B * ntile), dim3(64 * SEG_NG), 0, st, lam, 0, SEG, B, M, nseg, ntile,
+        hipLaunchKernelGGL(k_diag_seg_carry, dim3(B * ntile * (64 / SEG_CT)), dim3(SEG_NG * SEG_CT), 0, st, lam, 0, SEG, B,
+                           M, nseg, ntile,
                            (const float2 *)agg, carry);
     }
     DEER_LAUNCH_CHECK("k_diag_seg_carry");
@@ -1111,7 +1281,8 @@ int launch_diag_adjoint(int B, int T, int M, int K, const float *lam, const floa
         DEER_LAUNCH_CHECK("k_diag_rseg");
         {
             KTimer _kt("k_diag_seg_carry_rev", st);
-            hipLaunchKernelGGL(k_diag_seg_carry, dim3(B * nt64), dim3(64 * SEG_NG), 0, st, lam, 1, S, B, M, nseg, nt64,
+            hipLaunchKernelGGL(k_diag_seg_carry, dim3(B * nt64 * (64 / SEG_CT)), dim3(SEG_NG * SEG_CT), 0, st, lam, 1, S,
+                               B, M, nseg, nt64,
                                (const float2 *)agg, carry);
         }
         DEER_LAUNCH_CHECK("k_diag_seg_carry<rev>");

@@ -95,6 +95,26 @@ def test_diag_fused_projection_and_fused_gradients(B, T, M, K):
     assert rel_inf(_c(out2["grads"]["Bc"].cpu().numpy()), gr["Bc"]) < TOL
 
 
+@pytest.mark.parametrize("B,T,M,K", [(2, 4096, 64, 3), (1, 70000, 8, 2), (3, 1537, 33, 4), (1, 600, 64, 1),
+                                     (2, 512, 16, 3), (1, 513, 64, 3)])
+@pytest.mark.parametrize("mfma", ["1", "0"])
+def test_diag_forward_segment_aggregates(B, T, M, K, mfma, monkeypatch):
+    """Forward scan: the segment aggregates from the matrix-core product of the powers
+    lam^{63-k} with the transposed inputs (combined with lam^{64 (7 - a)} Bc), and from the
+    lane-per-channel walk, both against the sequential oracle; full and partial last segments,
+    |lam| close to 1."""
+    monkeypatch.setenv("DEER_DIAG_AGG_MFMA", mfma)
+    rng = np.random.default_rng(7 * T + M + K)
+    lam = (rng.uniform(0.99, 0.9999, M) * np.exp(1j * rng.uniform(0, np.pi / 4, M))).astype(np.complex64)
+    Bc = ((rng.standard_normal((M, K)) + 1j * rng.standard_normal((M, K))) / np.sqrt(2 * K)).astype(np.complex64)
+    x = rng.standard_normal((B, T + 1, K)).astype(np.float32)
+    m = {"kind": "diag_ssm", "lam": lam, "Bc": Bc}
+    say("deer_solve diag segment aggregates", B, T, M, K, mfma)
+    res = D.deer_solve(m, x, 0.0, 0)
+    h_ref = O.diag_scan(lam, O.diag_ssm_inputs({"Bc": Bc}, x))
+    assert rel_inf(_c(res["z"].cpu().numpy()), h_ref) < TOL
+
+
 @pytest.mark.parametrize("B,T,M,K,g_real,seg", [(1, 1, 1, 1, True, 0), (1, 5, 3, 2, False, 0),
                                                 (2, 511, 16, 3, True, 64), (1, 1025, 17, 4, False, 128),
                                                 (3, 2049, 64, 3, True, 192), (2, 5000, 70, 1, True, 0),

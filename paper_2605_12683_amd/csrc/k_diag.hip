@@ -632,13 +632,22 @@ __global__ __launch_bounds__(SEG_NG * SEG_CT) void k_diag_seg_carry(const float 
 // and R for the 64 channels (real parts in rows 0..63, imaginary parts in rows 64..127) and
 // the 32 columns (a, j) is one [128 x 64] x [64 x 32] product: A operand = the powers
 // lam^{63 - k} (LDS, formed once per block in float64), B operand = the segment's inputs
-// (LDS, transposed to [column 4 a + j][k]).  The k order is permuted as in the read-out (k-step
+// (registers).  The k order is permuted as in the read-out (k-step
 // (jj, q) of lane group g is k = 16 jj + 4 g + q) so that one 16-byte LDS read gives four
 // k-steps of either operand.  The epilogue multiplies every column by lam^{64 (7 - a)} Bc_j
 // and sums the 16 columns of a tile across its lanes.  A wave takes one segment at a time; a
 // partial last segment gets an aggregate that is never used (the carries stop before it).
 // ---------------------------------------------------------------------------------------
 constexpr int AGW = 4;        // waves (segments in flight) per block
+
+// sum over the 16 lanes of a DPP row, in every lane of it (row rotations by 8, 4, 2, 1)
+__device__ __forceinline__ float row16_sum(float v) {
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xF, 0xF, true));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xF, 0xF, true));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x122, 0xF, 0xF, true));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x121, 0xF, 0xF, true));
+    return v;
+}
 constexpr int AQS = 68;       // LDS row stride of the powers and of the transposed inputs
 
 __global__ __launch_bounds__(AGW * 64) void k_diag_seg_agg(const float *__restrict__ lam, const float *__restrict__ Bc,
@@ -646,7 +655,6 @@ __global__ __launch_bounds__(AGW * 64) void k_diag_seg_agg(const float *__restri
                                                            int nseg, float2 *__restrict__ agg) {
     static_assert(SEG == 512, "8 blocks of 64 steps per segment");
     __shared__ __align__(16) float qs[128][AQS];           // lam^{63-k}: re rows 0..63, im rows 64..127
-    __shared__ __align__(16) float us[AGW][32][AQS];       // inputs [4 a + j][k] of each wave's segment
     __shared__ float2 pw[64][8], bcs[64][4];                // lam^{64 (7 - a)}, Bc_j
     const int tid = threadIdx.x;
     // powers in float64: a thread takes 8 consecutive k of one channel (one power, then 7 products)
@@ -678,32 +686,33 @@ __global__ __launch_bounds__(AGW * 64) void k_diag_seg_agg(const float *__restri
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, c = lane & 15;
     const long total = (long)B * nseg;
     const long stride = (long)gridDim.x * AGW;
-    // inputs of a segment: lane l holds steps t0 + 8 l .. t0 + 8 l + 7 (block a = l / 8,
-    // k = 8 (l % 8) + i), loaded a segment ahead into registers
-    float nx[8][4];
+    // B operands of a segment straight from the inputs: k-step (jj, q) of lane (g, c) in column
+    // tile J is input j = c % 4 of step t0 + 64 a + 16 jj + 4 g + q, a = 4 J + c / 4 (zero past the
+    // sequence and for j >= K), loaded into registers at the start of the segment (the other
+    // waves of the CU cover the wait)
+    float nb[2][4][4];
+    const int jin = c & 3;
     auto fetch = [&](long sid) {
         const bool in = sid < total;
         const int b = in ? (int)(sid / nseg) : 0, seg = in ? (int)(sid % nseg) : 0;
         const int t0 = seg * SEG;
-        const int nrow = in ? min(8, T - t0 - 8 * lane) : 0;   // steps of this lane inside the sequence
-        const float *ur = u + ((long)b * (T + 1) + t0 + 8 * lane) * K;
+        const float *ub = u + (long)b * (T + 1) * K;
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+        for (int J = 0; J < 2; ++J)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) nx[i][j] = (i < nrow && j < K) ? ur[i * K + j] : 0.f;
+            for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int t = t0 + 64 * (4 * J + (c >> 2)) + 16 * jj + 4 * g + q;
+                    const bool ok = in && t < T && jin < K;
+                    nb[J][jj][q] = ok ? ub[(long)t * K + jin] : 0.f;
+                }
     };
-    long sid = (long)blockIdx.x * AGW + wv;
-    fetch(sid);
-    for (; sid < total; sid += stride) {
-        {
-            const int a = lane >> 3, k0 = 8 * (lane & 7);
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) us[wv][4 * a + j][k0 + i] = nx[i][j];
-        }
-        wave_lds_sync();
-        fetch(sid + stride);   // in flight during this segment's products
+    for (long sid = (long)blockIdx.x * AGW + wv; sid < total; sid += stride) {
+        fetch(sid);
+        // the powers are read from LDS k-block by k-block inside the loop (kept out of registers
+        // across segments, which leaves room for three waves per SIMD)
+        asm volatile("" ::: "memory");
         v4f acc[8][2];
 #pragma unroll
         for (int I = 0; I < 8; ++I) acc[I][0] = acc[I][1] = (v4f){0.f, 0.f, 0.f, 0.f};
@@ -713,7 +722,7 @@ __global__ __launch_bounds__(AGW * 64) void k_diag_seg_agg(const float *__restri
 #pragma unroll
             for (int I = 0; I < 8; ++I) aq[I] = *reinterpret_cast<const float4 *>(&qs[16 * I + c][16 * jj + 4 * g]);
 #pragma unroll
-            for (int J = 0; J < 2; ++J) bq[J] = *reinterpret_cast<const float4 *>(&us[wv][16 * J + c][16 * jj + 4 * g]);
+            for (int J = 0; J < 2; ++J) bq[J] = make_float4(nb[J][jj][0], nb[J][jj][1], nb[J][jj][2], nb[J][jj][3]);
             // 16 independent accumulators between two products into the same one
 #pragma unroll
             for (int J = 0; J < 2; ++J)
@@ -732,8 +741,6 @@ __global__ __launch_bounds__(AGW * 64) void k_diag_seg_agg(const float *__restri
 #pragma unroll
                 for (int I = 0; I < 8; ++I) acc[I][J] = mfma16x16x4(aq[I].w, bq[J].w, acc[I][J]);
         }
-        // the next segment's inputs may overwrite us once every lane has read it
-        wave_lds_sync();
         // epilogue: lane (g, c) holds rows 16 I + 4 g + r (channel 16 (I % 4) + 4 g + r, real part
         // for I < 4, imaginary for I >= 4) of columns 16 J + c = (a = 4 J + c / 4, j = c % 4)
         float sr[4][4], si[4][4];
@@ -755,14 +762,12 @@ __global__ __launch_bounds__(AGW * 64) void k_diag_seg_agg(const float *__restri
                 si[I][r] = xi;
             }
 #pragma unroll
-        for (int off = 1; off < 16; off <<= 1)
+        for (int I = 0; I < 4; ++I)
 #pragma unroll
-            for (int I = 0; I < 4; ++I)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    sr[I][r] += __shfl_xor(sr[I][r], off, 64);
-                    si[I][r] += __shfl_xor(si[I][r], off, 64);
-                }
+            for (int r = 0; r < 4; ++r) {
+                sr[I][r] = row16_sum(sr[I][r]);
+                si[I][r] = row16_sum(si[I][r]);
+            }
         if (c == 0) {
 #pragma unroll
             for (int I = 0; I < 4; ++I)
@@ -814,7 +819,7 @@ static int launch_diag_seg(int B, int T, int M, const float *lam, const float *B
         // segment aggregates on the matrix cores: a few blocks per CU, each forming the powers once
         const long segs = (long)B * nseg;
         const long want = (segs + AGW - 1) / AGW;
-        const int gridm = (int)(want < 512 ? want : 512);
+        const int gridm = (int)(want < 768 ? want : 768);   // three blocks per CU
         KTimer _kt("k_diag_seg_reduce", st);
         hipLaunchKernelGGL(k_diag_seg_agg, dim3(gridm), dim3(AGW * 64), 0, st, lam, Bc, u, B, T, M, K, nseg, agg);
     } else {

@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdeer.so")
 SOURCES = ["deer_api.hip", "k_plrnn.hip", "k_diag.hip", "k_dense.hip", "k_shallow.hip", "k_readout.hip", "k_seq.hip", "k_quasi.hip", "k_small.hip", "k_train.hip", "deer_noalloc.hip", "k_obs.hip", "k_big.hip", "k_shfused.hip"]
-HEADERS = ["common.h", "launch.h", os.path.join("..", "..", "include", "deer.h")]
+HEADERS = ["common.h", "launch.h", "newton_ctl.h", "row16.h", os.path.join("..", "..", "include", "deer.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

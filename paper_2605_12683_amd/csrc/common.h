@@ -81,6 +81,28 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     return v;
 }
 
+// Buffer resource with a wave-uniform base: an access adds a per-lane byte offset (VGPR) and a
+// wave-uniform byte offset (SGPR).  A lane offset of 2^31 or more is outside the resource: a
+// load from it returns zero and a store to it is dropped.
+constexpr uint32_t kOffLane = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t wave_rsrc(const void *base) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ uint32_t bload_u(__amdgpu_buffer_rsrc_t rs, uint32_t voff, int soff) {
+    return __builtin_amdgcn_raw_buffer_load_b32(rs, (int)voff, soff, 0);
+}
+__device__ __forceinline__ float bload(__amdgpu_buffer_rsrc_t rs, uint32_t voff, int soff) {
+    return __uint_as_float(bload_u(rs, voff, soff));
+}
+__device__ __forceinline__ void bstore_u(__amdgpu_buffer_rsrc_t rs, uint32_t v, uint32_t voff, int soff) {
+    __builtin_amdgcn_raw_buffer_store_b32(v, rs, (int)voff, soff, 0);
+}
+// The same over `bytes` bytes from base (bytes < 2^31): an access at or past the end reads zero
+// and a store there is dropped.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t bounded_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 // forced input of step s (array index) for latent i:
 //   s == 0: z0 (or [x_0; 0] when z0 is null);  s >= 1: fl(fl(p*z_{s-1}) + fl(a*zbar_s))
 // The two iterate buffers of the safeguarded Newton loop: sequence b's current iterate is in

@@ -208,6 +208,13 @@ static bool pass_fusion_allowed() {
     return !e || atoi(e) != 0;
 }
 
+// DEER_QUASI_FUSED=0 keeps the vanilla quasi-DEER passes of the adaptive loop in separate
+// kernels (a test override)
+static bool quasi_fusion_allowed() {
+    const char *e = getenv("DEER_QUASI_FUSED");
+    return !e || atoi(e) != 0;
+}
+
 // Chunk length of the dense scans: enough chains to fill the machine (about 2048 waves),
 // and a bounded number of chunks per sequence so that the two-level carry pass stays short
 // (1024 for MP <= 32, 512 for MP = 64, whose group pass composes 64 x 64 maps).
@@ -398,6 +405,8 @@ static ShWs carve_sh(void *ws, int B, int T, int M, int L, int op, bool need_g, 
 // does not keep it, and the partial sums of the shallow gradient kernel)
 struct QuasiWs {
     float *rhs, *coef, *P, *v, *carry;
+    float *P2, *v2;      // vanilla solve: the second set of chunk aggregates of the fused passes
+    double *gm, *gm2;    // and the two sets of group maps [B][chunks / group][2][MP]
     NewtonCtl ctl;
     float *gpart;
     double *gpart2;
@@ -406,11 +415,21 @@ struct QuasiWs {
     int C, ncs, MP;
 };
 
+// The vanilla solve is carved for the fused passes (chunk count per sequence padded to a whole
+// number of the pass kernel's groups; the separate kernels take the empty padding chunks too).
 static QuasiWs carve_quasi(void *ws, int B, int T, int M, int L, int op, size_t *bytes) {
     QuasiWs w{};
     w.MP = padded_dim(M);
     w.C = qdeer_chunk_len(B, T, M);
     w.ncs = (T + w.C - 1) / w.C;
+    const bool fused = op == DEER_OP_SOLVE && L == 0;
+    const int GS = fused ? qdeer_pass_group(M) : 1;
+    if (fused)
+        while (w.ncs > qdeer_pass_max_chunks(M)) {
+            w.C *= 2;
+            w.ncs = (T + w.C - 1) / w.C;
+        }
+    w.ncs = (w.ncs + GS - 1) / GS * GS;
     const size_t nch = (size_t)B * w.ncs;
     Carver c(ws);
     w.coef = c.take<float>((size_t)B * T * M);
@@ -421,6 +440,13 @@ static QuasiWs carve_quasi(void *ws, int B, int T, int M, int L, int op, size_t 
     if (op == DEER_OP_SOLVE) {
         w.rhs = c.take<float>((size_t)B * T * M);
         w.ctl = carve_ctl(c, B, (size_t)T * M, nch);
+        if (fused) {
+            const size_t ngm = (size_t)B * (w.ncs / GS) * 2 * w.MP;
+            w.P2 = c.take<float>(nch * w.MP);
+            w.v2 = c.take<float>(nch * w.MP);
+            w.gm = c.take<double>(ngm);
+            w.gm2 = c.take<double>(ngm);
+        }
     } else if (L > 0) {
         w.lam = c.take<float>((size_t)B * T * M);
         int nb = 0;
@@ -1130,8 +1156,27 @@ static int solve_quasi(const deer_model *m, const deer_forcing *f, const deer_so
     std::vector<int> act(B, 1), it(B, 0);
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
-    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *,
-                      uint32_t) -> int {
+    // vanilla PLRNN, adaptive loop: one kernel per pass (the fix-up of the previous update and
+    // the chunk aggregates of the next, with the pass-end control)
+    NewtonCtl ctl = w.ctl;
+    const bool qf = L == 0 && o->fixed_iters <= 0 && (size_t)(T + 1) * m->M * 4 < ((size_t)1 << 31) &&
+                    quasi_fusion_allowed();   // a sequence's rows addressed with 32-bit offsets
+    if (qf) {
+        ctl.fused = true;
+        ctl.nd.pv = ctl.pv;
+        ctl.lead = 1;
+        uint32_t *mark_unused = nullptr;
+        if ((rc = host_block(B, ctl.nd, &mark_unused))) return rc;
+    }
+    const FusedCtl fc{ctl.nd, ctl.seq, o->tol, o->step_bound == 0.f ? kDefaultStepBound : o->step_bound, kDamp};
+    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *mark,
+                      uint32_t pass_no) -> int {
+        if (qf) {   // aggregates alternate between the two sets
+            const bool odd = pass_no & 1u;
+            return launch_qdeer_pass(a, zb, za, odd ? w.P2 : w.P, odd ? w.v2 : w.v, odd ? w.gm2 : w.gm,
+                                     odd ? w.P : w.P2, odd ? w.v : w.v2, odd ? w.gm : w.gm2, w.C, w.ncs, fc, mark,
+                                     pass_no, st);
+        }
         if (L == 0)
             return launch_qdeer_update(a, zb, za, zsel, dact, gam, w.rhs, w.coef, w.P, w.v, w.carry,
                                        w.ctl.chain_bits, w.C, w.ncs, st);
@@ -1142,7 +1187,7 @@ static int solve_quasi(const deer_model *m, const deer_forcing *f, const deer_so
         return launch_qdeer_scan_fwd(B, T, m->M, x, f->n_forced, zb, za, zsel, dact, w.rhs, w.coef, w.P, w.v, w.carry,
                                      w.ctl.chain_bits, w.C, w.ncs, st);
     };
-    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ncs, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
+    if ((rc = newton_loop(o, B, (size_t)T * m->M, w.ncs, ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
         rc = L == 0 ? launch_resjac_plrnn(a, z, nullptr, nullptr, nullptr, masks, nullptr, st)
                     : launch_resjac_shplrnn(sa, z, nullptr, nullptr, nullptr, nullptr, masks, nullptr, st);

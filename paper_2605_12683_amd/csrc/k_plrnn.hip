@@ -16,6 +16,8 @@
 
 #include "common.h"
 #include "launch.h"
+#include "newton_ctl.h"
+#include "row16.h"
 
 namespace deer {
 
@@ -590,115 +592,6 @@ __device__ __forceinline__ void carry16_fetch(const float *__restrict__ Pc, cons
 // residual and the masks stay in registers: the fix-up forms them again from z and x.
 // ---------------------------------------------------------------------------------------
 
-// lane l of each 16-lane row receives v from lane row_src(l, K) of the same row
-template <int K>
-__device__ __forceinline__ int row_ror_i(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, 0x120 + K, 0xF, 0xF, true);
-}
-
-// source lane (within the row) of rotation k, k = 0..15
-__device__ __forceinline__ void row_sources(int c, int (&src)[16]) {
-    src[0] = c;
-    src[1] = row_ror_i<1>(c);   src[2] = row_ror_i<2>(c);   src[3] = row_ror_i<3>(c);
-    src[4] = row_ror_i<4>(c);   src[5] = row_ror_i<5>(c);   src[6] = row_ror_i<6>(c);
-    src[7] = row_ror_i<7>(c);   src[8] = row_ror_i<8>(c);   src[9] = row_ror_i<9>(c);
-    src[10] = row_ror_i<10>(c); src[11] = row_ror_i<11>(c); src[12] = row_ror_i<12>(c);
-    src[13] = row_ror_i<13>(c); src[14] = row_ror_i<14>(c); src[15] = row_ror_i<15>(c);
-}
-
-// sum_k w[k] * v(row_src(lane, k)): with w[k] = W[i][row_src(i, k)] this is (W v)_i for the
-// vector v held by the 16 lanes of the row.  One multiply-add with a DPP row rotation of v per
-// term (the compiler does not fuse a rotation into v_fmac by itself); the leading s_nop covers
-// the wait a DPP read needs after a VALU write of v.  All 64 lanes must be active.
-#define DEER_RR(k) " row_ror:" #k " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
-__device__ __forceinline__ float row16_dot(const float (&w)[16], float v) {
-    float a0, a1;
-    asm volatile(
-        "s_nop 1\n"
-        "v_mul_f32_e32 %0, %2, %3\n"
-        "v_mul_f32_dpp %1, %2, %4" DEER_RR(1)
-        "v_fmac_f32_dpp %0, %2, %5" DEER_RR(2)
-        "v_fmac_f32_dpp %1, %2, %6" DEER_RR(3)
-        "v_fmac_f32_dpp %0, %2, %7" DEER_RR(4)
-        "v_fmac_f32_dpp %1, %2, %8" DEER_RR(5)
-        "v_fmac_f32_dpp %0, %2, %9" DEER_RR(6)
-        "v_fmac_f32_dpp %1, %2, %10" DEER_RR(7)
-        "v_fmac_f32_dpp %0, %2, %11" DEER_RR(8)
-        "v_fmac_f32_dpp %1, %2, %12" DEER_RR(9)
-        "v_fmac_f32_dpp %0, %2, %13" DEER_RR(10)
-        "v_fmac_f32_dpp %1, %2, %14" DEER_RR(11)
-        "v_fmac_f32_dpp %0, %2, %15" DEER_RR(12)
-        "v_fmac_f32_dpp %1, %2, %16" DEER_RR(13)
-        "v_fmac_f32_dpp %0, %2, %17" DEER_RR(14)
-        "v_fmac_f32_dpp %1, %2, %18" DEER_RR(15)
-        : "=&v"(a0), "=&v"(a1)
-        : "v"(v), "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "v"(w[4]), "v"(w[5]), "v"(w[6]), "v"(w[7]), "v"(w[8]),
-          "v"(w[9]), "v"(w[10]), "v"(w[11]), "v"(w[12]), "v"(w[13]), "v"(w[14]), "v"(w[15]));
-    return a0 + a1;
-}
-
-// two independent row products W v0, W v1 (each summed exactly as row16_dot), interleaved so
-// that dependent multiply-adds are four instructions apart
-__device__ __forceinline__ void row16_dot2(const float (&w)[16], float v0, float v1, float &r0, float &r1) {
-    float a0, a1, b0, b1;
-    asm volatile(
-        "s_nop 1\n"
-        "v_mul_f32_e32 %0, %4, %6\n"
-        "v_mul_f32_e32 %2, %5, %6\n"
-        "v_mul_f32_dpp %1, %4, %7" DEER_RR(1)
-        "v_mul_f32_dpp %3, %5, %7" DEER_RR(1)
-        "v_fmac_f32_dpp %0, %4, %8" DEER_RR(2)
-        "v_fmac_f32_dpp %2, %5, %8" DEER_RR(2)
-        "v_fmac_f32_dpp %1, %4, %9" DEER_RR(3)
-        "v_fmac_f32_dpp %3, %5, %9" DEER_RR(3)
-        "v_fmac_f32_dpp %0, %4, %10" DEER_RR(4)
-        "v_fmac_f32_dpp %2, %5, %10" DEER_RR(4)
-        "v_fmac_f32_dpp %1, %4, %11" DEER_RR(5)
-        "v_fmac_f32_dpp %3, %5, %11" DEER_RR(5)
-        "v_fmac_f32_dpp %0, %4, %12" DEER_RR(6)
-        "v_fmac_f32_dpp %2, %5, %12" DEER_RR(6)
-        "v_fmac_f32_dpp %1, %4, %13" DEER_RR(7)
-        "v_fmac_f32_dpp %3, %5, %13" DEER_RR(7)
-        "v_fmac_f32_dpp %0, %4, %14" DEER_RR(8)
-        "v_fmac_f32_dpp %2, %5, %14" DEER_RR(8)
-        "v_fmac_f32_dpp %1, %4, %15" DEER_RR(9)
-        "v_fmac_f32_dpp %3, %5, %15" DEER_RR(9)
-        "v_fmac_f32_dpp %0, %4, %16" DEER_RR(10)
-        "v_fmac_f32_dpp %2, %5, %16" DEER_RR(10)
-        "v_fmac_f32_dpp %1, %4, %17" DEER_RR(11)
-        "v_fmac_f32_dpp %3, %5, %17" DEER_RR(11)
-        "v_fmac_f32_dpp %0, %4, %18" DEER_RR(12)
-        "v_fmac_f32_dpp %2, %5, %18" DEER_RR(12)
-        "v_fmac_f32_dpp %1, %4, %19" DEER_RR(13)
-        "v_fmac_f32_dpp %3, %5, %19" DEER_RR(13)
-        "v_fmac_f32_dpp %0, %4, %20" DEER_RR(14)
-        "v_fmac_f32_dpp %2, %5, %20" DEER_RR(14)
-        "v_fmac_f32_dpp %1, %4, %21" DEER_RR(15)
-        "v_fmac_f32_dpp %3, %5, %21" DEER_RR(15)
-        : "=&v"(a0), "=&v"(a1), "=&v"(b0), "=&v"(b1)
-        : "v"(v0), "v"(v1), "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "v"(w[4]), "v"(w[5]), "v"(w[6]), "v"(w[7]),
-          "v"(w[8]), "v"(w[9]), "v"(w[10]), "v"(w[11]), "v"(w[12]), "v"(w[13]), "v"(w[14]), "v"(w[15]));
-    r0 = a0 + a1;
-    r1 = b0 + b1;
-}
-#undef DEER_RR
-
-// Buffer resource with a wave-uniform base: an access adds a per-lane byte offset (VGPR) and a
-// wave-uniform byte offset (SGPR).  A lane offset of 2^31 or more is outside the resource: a
-// load from it returns zero and a store to it is dropped.
-constexpr uint32_t kOffLane = 0x80000000u;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t wave_rsrc(const void *base) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, 0x7fffffff, 0x00020000);
-}
-__device__ __forceinline__ uint32_t bload_u(__amdgpu_buffer_rsrc_t rs, uint32_t voff, int soff) {
-    return __builtin_amdgcn_raw_buffer_load_b32(rs, (int)voff, soff, 0);
-}
-__device__ __forceinline__ float bload(__amdgpu_buffer_rsrc_t rs, uint32_t voff, int soff) {
-    return __uint_as_float(bload_u(rs, voff, soff));
-}
-__device__ __forceinline__ void bstore_u(__amdgpu_buffer_rsrc_t rs, uint32_t v, uint32_t voff, int soff) {
-    __builtin_amdgcn_raw_buffer_store_b32(v, rs, (int)voff, soff, 0);
-}
 
 __device__ __forceinline__ int rfl_i(int v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ float rfl_f(float v) { return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v))); }
@@ -1158,69 +1051,6 @@ __global__ __launch_bounds__(64 * WPB) void k_newton_product_plrnn16(
         }
     }
     if (okc) vout[(size_t)id * 16 + c] = u;
-}
-
-// Convergence test and update safeguard of one pass for sequence b from its maxima e = max
-// |Delta| bits and zm = max |z| bits: accept the update (flip sel, count it, relax the damping,
-// freeze the sequence once max|Delta| < tol), or reject it (keep sel, raise the damping:
-// 1 - gamma = first, then x grow up to 1 = the fixed-point step); a non-finite fixed-point step
-// ends the sequence.
-// tag: with nd.pv, the number of the pass that may use the aggregates the caller's kernel
-// formed for the accepted iterate (it is stored when the update is kept and the sequence goes on)
-__device__ __forceinline__ void seq_decide(int b, uint32_t e, uint32_t zm, const NewtonDev &nd, float tol, float bound,
-                                           const NewtonDamp &dp, uint32_t tag = 0u) {
-    const float ef = __uint_as_float(e), zf = __uint_as_float(zm);
-    const bool fin = e < 0x7f800000u;
-    float om = nd.om[b];
-    const bool keep = fin && (bound < 0.f || om >= 1.f || ef <= bound * (1.f + zf));
-    // a stopped sequence: device control block, then the host block (act last)
-    auto stop = [&](int it, int status) {
-        nd.act[b] = 0;
-        nd.status[b] = status;
-        if (nd.hact) {
-            nd.hit[b] = it;
-            nd.hnorm[b] = ef;
-            nd.hstat[b] = status;
-            __hip_atomic_store(nd.hact + b, 0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
-        }
-    };
-    if (keep) {
-        nd.sel[b] ^= 1;
-        const int it = nd.it[b] + 1;
-        nd.it[b] = it;
-        nd.norm[b] = ef;
-        if (om > 0.f) om = om / dp.shrink < dp.floor ? 0.f : om / dp.shrink;
-        if (ef < tol) stop(it, 1);
-        else if (nd.pv) nd.pv[b] = tag;
-    } else if (om >= 1.f) {
-        nd.norm[b] = ef;
-        stop(nd.it[b], 2);
-    } else {
-        om = om == 0.f ? dp.first : fminf(1.f, om * dp.grow);
-    }
-    nd.om[b] = om;
-    nd.gamma[b] = 1.f - om;
-}
-
-// Arrival of `cnt` chains of sequence b with maxima e, zm (see FusedCtl).  Device-scope atomics
-// meet at one coherence point across the XCDs; each maximum is returned (so performed) before
-// the count is raised, so the chain that completes the count reads the final maxima.
-__device__ __forceinline__ void seq_arrive(const FusedCtl &fc, int b, int cnt, int ncs, uint32_t e, uint32_t zm,
-                                           uint32_t tag = 0u) {
-    uint32_t *blk = fc.seq + (size_t)b * kSeqWords;   // count | max |Delta| | max |z|, 128 bytes apart
-    const uint32_t r1 = __hip_atomic_fetch_max(blk + 32, e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint32_t r2 = __hip_atomic_fetch_max(blk + 64, zm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    // the count may only move once both maxima are in: the increment depends on their return
-    // values (|x| bits are below 2^31, so the added term is zero)
-    const uint32_t old = __hip_atomic_fetch_add(blk, (uint32_t)cnt + ((r1 | r2) >> 31), __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-    if (old + (uint32_t)cnt != (uint32_t)ncs) return;
-    const uint32_t ef = __hip_atomic_load(blk + 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint32_t zf = __hip_atomic_load(blk + 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    seq_decide(b, ef, zf, fc.nd, fc.tol, fc.bound, fc.dp, tag);
-    __hip_atomic_store(blk + 32, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(blk + 64, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(blk, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // M <= 16 forward fix-up.  The residual and the masks are formed again here from z and x (the

@@ -16,11 +16,15 @@
 //   k_qdeer_fixup     forward: z + Delta to the other iterate buffer, per-chain max|Delta| and
 //                     max|z|; reverse: lam (optional) and the gradient partial sums of the
 //                     chain, dW_ij += lam_i relu(z~_j), dA_i += lam_i z~_i, dh_i += lam_i
+//   k_qdeer_pass      the adaptive loop's pass in one kernel: the fix-up of one update and the
+//                     chunk aggregates of the next, with the pass-end control
 //
 // Lanes: a wave holds 64 / MP chains of MP lanes (lane = latent), MP in {16, 32, 64}; the
 // ReLU row of a step goes through LDS when the lanes of a chain need each other's values.
 #include "common.h"
 #include "launch.h"
+#include "newton_ctl.h"
+#include "row16.h"
 
 namespace deer {
 
@@ -319,6 +323,301 @@ __global__ __launch_bounds__(64) void k_qdeer_fixup_fwd(const float *__restrict_
 }
 
 // ---------------------------------------------------------------------------------------
+// One kernel per pass of the adaptive loop.  A block takes a group of GS = QF_WPB (64 / MP)
+// consecutive chunks of one sequence (the chunk count per sequence is padded to a multiple of
+// GS with empty chunks) and runs, per chunk:
+//   1. when the sequence's aggregates of the previous kernel belong to its current iterate
+//      (nd.pv == pass_no): the chunk's carry, walked in float64 over the group maps of the
+//      groups before it and the chunk aggregates before it in its group, then the fix-up
+//      Delta_s = coef_s Delta_{s-1} - r_s with r and coef formed again from z (the same
+//      operations as the separate kernels), z + Delta written to the other iterate buffer;
+//   2. the chunk aggregates of the next update at the new iterate (or at the current one when
+//      step 1 did not run): prod coef and the local solution from zero, with the damping that
+//      an accepted update leads to, and the group map of the block (float64);
+//   3. the pass-end control of step 1's update (seq_arrive), which also records in nd.pv that
+//      the aggregates just formed belong to the accepted iterate.
+// Step 2 at a chunk's first step needs the new iterate at the step before the chunk: that is
+// z + carry, and the chunk before puts exactly that value there (it forms this chunk's carry
+// with the same float64 operations on the same operands instead of taking the end of its own
+// recurrence), so no wave waits for another.  Aggregates alternate between two buffers.
+// ---------------------------------------------------------------------------------------
+// Products (W relu(zt_q))_i for the TS steps q of a tile, lane = latent i of its chain.  MP = 16:
+// formed here by DPP row rotations into dq (w: the row's weights in rotation order); else the
+// ReLU rows go to the wave's LDS rows, and q_tile_dot reads product q where it is consumed (all
+// of them at once would hold every operand in registers).
+template <int MP, int TS>
+__device__ __forceinline__ void q_tile_rows(const float (&zt)[TS], const float (&w)[MP], float (*lr)[64], int lane,
+                                            float (&dq)[TS]) {
+    if constexpr (MP == 16) {
+#pragma unroll
+        for (int q = 0; q < TS; q += 2)
+            row16_dot2(w, zt[q] > 0.f ? zt[q] : 0.f, zt[q + 1] > 0.f ? zt[q + 1] : 0.f, dq[q], dq[q + 1]);
+    } else {
+#pragma unroll
+        for (int q = 0; q < TS; ++q) lr[q][lane] = zt[q] > 0.f ? zt[q] : 0.f;
+        wave_lds_sync();
+    }
+}
+template <int MP, int TS>
+__device__ __forceinline__ float q_tile_dot(const float (&dq)[TS], const float (&w)[MP], float (*lr)[64], int n, int q) {
+    if constexpr (MP == 16) return dq[q];
+    else return q_dot<MP>(lr[q], n, w);
+}
+
+constexpr int QF_WPB = 8;   // waves per block
+constexpr int QF_TS = 8;    // steps per tile
+constexpr int QF_MAXG = 32; // groups per sequence at most
+
+template <int MP>
+__global__ __launch_bounds__(64 * QF_WPB) void k_qdeer_pass(
+    const float *__restrict__ A, const float *__restrict__ W, const float *__restrict__ h, float alpha, int N,
+    const float *__restrict__ x, const float *__restrict__ z0, float *zbuf, float *zalt, int T, int M, int C, int ncs,
+    const float *__restrict__ Pin, const float *__restrict__ vin, const double *__restrict__ gin,
+    float *__restrict__ Pout, float *__restrict__ vout, double *__restrict__ gout, FusedCtl fc, uint32_t *mark,
+    uint32_t pass_no, int tw) {
+    constexpr int NCH = 64 / MP, GS = QF_WPB * NCH, TS = QF_TS;
+    __shared__ __align__(16) float rl[MP == 16 ? 1 : QF_WPB][TS][64];   // ReLU rows of a tile, per wave (MP > 16)
+    __shared__ float sW[MP * MP];
+    __shared__ float sag[2][GS][MP];                      // the previous kernel's chunk aggregates of the group
+    __shared__ float sagn[2][GS][MP];                     // the next update's
+    __shared__ double sG[2][QF_MAXG][MP];                 // group maps of the groups up to this one
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, n = lane / MP, i = lane % MP;
+    if (mark && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(mark, pass_no, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    const NewtonDev &nd = fc.nd;
+    const int ngm = ncs / GS;
+    const int b = blockIdx.x / ngm, grp = blockIdx.x - b * ngm;
+    if (nd.act[b] == 0) return;   // the whole block
+    const bool have = nd.pv[b] == pass_no;
+    const int sel = nd.sel[b];
+    const float gam = nd.gamma[b];
+    float omn = nd.om[b];   // the damping of the next update if this one is kept
+    if (omn > 0.f) omn = omn / fc.dp.shrink < fc.dp.floor ? 0.f : omn / fc.dp.shrink;
+    const float gnext = have ? 1.f - omn : gam;
+    const float *const zc = sel ? zalt : zbuf;   // current iterate
+    float *const zn = sel ? zbuf : zalt;         // the update's output
+    const int kg = wv * NCH + n;                 // this lane's chunk within the group
+    const int c = grp * GS + kg;
+    const int s0 = c * C;
+    const int len = max(min(s0 + C, T) - s0, 0);  // 0: a padding chunk
+    int maxlen = len;                              // the wave's tile loop is uniform
+#pragma unroll
+    for (int off = 32; off >= MP; off >>= 1) maxlen = max(maxlen, __shfl_xor(maxlen, off, 64));
+    const bool iok = i < M, forced = i < N;
+    const size_t zrow = (size_t)b * T;
+    const float *xs = x + (size_t)b * (T + 1) * N;
+    // buffer resources over the sequence's rows (a load past its end reads zero): a lane's byte
+    // offset is that of its chunk's first step, a tile step adds a wave-uniform offset
+    const auto rzc = bounded_rsrc(zc + zrow * M, (uint32_t)T * M * 4u);
+    const auto rzn = bounded_rsrc(zn + zrow * M, (uint32_t)T * M * 4u);
+    const auto rx = bounded_rsrc(xs, (uint32_t)(T + 1) * N * 4u);
+    const uint32_t vz = (iok && len > 0) ? 4u * ((uint32_t)s0 * M + i) : kOffLane;
+    const uint32_t vx = (forced && len > 0) ? 4u * ((uint32_t)s0 * N + i) : kOffLane;
+    // the first tile's inputs and z_{s0-1} of the current iterate (the initial state at s0 = 0,
+    // taken as the forced state) go out first
+    float zq[TS], xq[TS];
+    auto load = [&](int t0) {
+#pragma unroll
+        for (int q = 0; q < TS; ++q) {
+            zq[q] = bload(rzc, vz, 4 * (t0 + q) * M);
+            xq[q] = bload(rx, vx, 4 * (t0 + q) * N);
+        }
+    };
+    load(0);
+    float zprev = 0.f;
+    if (iok && len > 0) {
+        if (s0 == 0) zprev = z0 ? z0[(size_t)b * M + i] : (forced ? xs[i] : 0.f);
+        else zprev = zc[(zrow + s0 - 1) * M + i];
+    }
+    // weights, and the previous kernel's aggregates this block walks, through LDS
+    for (int t = threadIdx.x; t < M * M; t += 64 * QF_WPB) sW[t] = W[t];
+    if (have) {
+        const float *Pg = Pin + ((size_t)b * ncs + (size_t)grp * GS) * MP;
+        const float *vg = vin + ((size_t)b * ncs + (size_t)grp * GS) * MP;
+        for (int t = threadIdx.x; t < GS * MP; t += 64 * QF_WPB) {
+            sag[0][t / MP][t % MP] = Pg[t];
+            sag[1][t / MP][t % MP] = vg[t];
+        }
+        const double *G = gin + (size_t)b * ngm * 2 * MP;
+        for (int t = threadIdx.x; t < (grp + 1) * MP; t += 64 * QF_WPB) {   // groups 0 .. grp
+            const int q = t / MP, j = t % MP;
+            sG[0][q][j] = G[(size_t)q * 2 * MP + j];
+            sG[1][q][j] = G[(size_t)q * 2 * MP + MP + j];
+        }
+    }
+    __syncthreads();
+    float wrow[MP];   // row i of W (MP = 16: in the order of the row rotations)
+    if constexpr (MP == 16) {
+        int src[16];
+        row_sources(i, src);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) wrow[k] = (iok && src[k] < M) ? sW[i * M + src[k]] : 0.f;
+    } else {
+#pragma unroll
+        for (int j = 0; j < MP; ++j) wrow[j] = (iok && j < M) ? sW[i * M + j] : 0.f;
+    }
+    const float Ai = iok ? A[i] : 0.f, Wii = iok ? sW[i * M + i] : 0.f, hi = (h && iok) ? h[i] : 0.f;
+    const float pi = q_p(i, N, alpha);
+    // ---- the chunk's carry and the next chunk's (float64 walks over the group maps before the
+    // group and the chunk aggregates before the chunk) ----
+    float D = 0.f, Dn = 0.f;
+    const bool usenext = have && s0 + C < T;   // the next chunk holds steps
+    if (have && iok) {
+        // operands read 8 at a time ahead of the dependent multiply-adds
+        double X = 0.0;
+        for (int q0 = 0; q0 < grp; q0 += 8) {
+            double gp[8], gv[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int q = min(q0 + k, grp - 1);
+                gp[k] = sG[0][q][i];
+                gv[k] = sG[1][q][i];
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                if (q0 + k < grp) X = fma(gp[k], X, gv[k]);
+        }
+        const double Xg = X;
+        for (int k0 = 0; k0 < kg; k0 += 8) {
+            float pp[8], vv[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int q = min(k0 + k, kg - 1);
+                pp[k] = sag[0][q][i];
+                vv[k] = sag[1][q][i];
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                if (k0 + k < kg) X = fma((double)pp[k], X, (double)vv[k]);
+        }
+        D = (float)X;
+        if (usenext) {   // the operations the next chunk forms its carry with
+            const double Xn = kg + 1 == GS ? fma(sG[0][grp][i], Xg, sG[1][grp][i])
+                                           : fma((double)sag[0][kg][i], X, (double)sag[1][kg][i]);
+            Dn = (float)Xn;
+        }
+    }
+    // z_{s0-1} of the iterate the next update is formed at (as the chunk before stores it)
+    float zpn = have ? zprev + D : zprev;
+    uint32_t emax = 0u, zmax = 0u;
+    float u = 0.f, Pn = 1.f;
+    float (*const lr)[64] = rl[MP == 16 ? 0 : wv];
+    // Branch-free tile bodies (the DPP products need every lane): a lane past its chunk's end
+    // keeps its recurrences and stores nothing; padding lanes (i >= M) read zeros, so their
+    // residuals, coefficients and Delta are zero.
+    for (int t0 = 0; t0 < maxlen; t0 += TS) {
+        float zv[TS], xv[TS];
+#pragma unroll
+        for (int q = 0; q < TS; ++q) {
+            zv[q] = zq[q];
+            xv[q] = xq[q];
+        }
+        if (t0 + TS < maxlen) load(t0 + TS);   // the next tile's inputs, in flight during this one
+        if (have) {
+            // residual and coefficients at the current iterate, then the fix-up
+            float zt[TS];
+#pragma unroll
+            for (int q = 0; q < TS; ++q) {
+                const int s = s0 + t0 + q;
+                const float fz = s <= tw ? xv[q] : __fadd_rn(__fmul_rn(pi, zprev), __fmul_rn(alpha, xv[q]));
+                zt[q] = (s == 0 || !forced) ? zprev : fz;
+                zprev = zv[q];
+            }
+            float dq[TS];
+            q_tile_rows<MP, TS>(zt, wrow, lr, lane, dq);
+#pragma unroll
+            for (int q = 0; q < TS; ++q) {
+                const int s = s0 + t0 + q;
+                const float F = fmaf(Ai, zt[q], q_tile_dot<MP, TS>(dq, wrow, lr, n, q)) + hi;
+                const float r = zv[q] - F;
+                const float cf = q_coef(zt[q], Ai, Wii, (forced && s <= tw) ? 0.f : pi, gam);
+                const bool st = t0 + q < len;
+                const float Dq = fmaf(cf, D, -r);
+                D = st ? Dq : D;
+                const float dap = (usenext && t0 + q == len - 1) ? Dn : D;
+                const float znew = zv[q] + dap;
+                bstore_u(rzn, __float_as_uint(znew), st ? vz : kOffLane, 4 * (t0 + q) * M);
+                const uint32_t ab = st ? abs_bits(dap) : 0u, zb = st ? abs_bits(zv[q]) : 0u;
+                emax = emax > ab ? emax : ab;
+                zmax = zmax > zb ? zmax : zb;
+                zv[q] = st ? znew : zv[q];
+            }
+            if constexpr (MP != 16) wave_lds_sync();   // the rows are read before they are rewritten
+        }
+        // the next update's residual and coefficients at the (new) iterate: chunk aggregates
+        {
+            float zt[TS];
+#pragma unroll
+            for (int q = 0; q < TS; ++q) {
+                const int s = s0 + t0 + q;
+                const float fz = s <= tw ? xv[q] : __fadd_rn(__fmul_rn(pi, zpn), __fmul_rn(alpha, xv[q]));
+                zt[q] = (s == 0 || !forced) ? zpn : fz;
+                zpn = zv[q];
+            }
+            float dq[TS];
+            q_tile_rows<MP, TS>(zt, wrow, lr, lane, dq);
+#pragma unroll
+            for (int q = 0; q < TS; ++q) {
+                const int s = s0 + t0 + q;
+                const float F = fmaf(Ai, zt[q], q_tile_dot<MP, TS>(dq, wrow, lr, n, q)) + hi;
+                const float r = zv[q] - F;
+                const float cf = q_coef(zt[q], Ai, Wii, (forced && s <= tw) ? 0.f : pi, gnext);
+                const bool st = t0 + q < len;
+                const float uq = fmaf(cf, u, -r), pq = Pn * cf;
+                u = st ? uq : u;
+                Pn = st ? pq : Pn;
+            }
+            if constexpr (MP != 16) wave_lds_sync();
+        }
+    }
+    if (!iok) {
+        u = 0.f;
+        Pn = 1.f;
+    }
+    __shared__ uint32_t smx[2][QF_WPB];
+    if (have) {
+        emax = wave_max_u32(emax);
+        zmax = wave_max_u32(zmax);
+        if (lane == 0) {
+            smx[0][wv] = emax;
+            smx[1][wv] = zmax;
+        }
+    }
+    // ---- chunk aggregates of the next update ----
+    const size_t e = ((size_t)b * ncs + c) * MP + i;
+    Pout[e] = Pn;
+    vout[e] = u;
+    sagn[0][kg][i] = Pn;
+    sagn[1][kg][i] = u;
+    __syncthreads();
+    // ---- pass-end control of the current update (once per block: its chunks share b) ----
+    if (threadIdx.x == 0) {
+        if (have) {
+            uint32_t em = smx[0][0], zm = smx[1][0];
+            for (int w = 1; w < QF_WPB; ++w) {
+                em = em > smx[0][w] ? em : smx[0][w];
+                zm = zm > smx[1][w] ? zm : smx[1][w];
+            }
+            seq_arrive(fc, b, GS, ncs, em, zm, pass_no + 1u);
+        } else {
+            // aggregates of the current iterate (nothing else of this sequence runs in this kernel)
+            nd.pv[b] = pass_no + 1u;
+        }
+    }
+    // ---- the group map of the next update ----
+    if (threadIdx.x >= MP) return;
+    double gp = 1.0, gv = 0.0;
+    for (int k = 0; k < GS; ++k) {
+        const double pk = (double)sagn[0][k][threadIdx.x];
+        gv = fma(pk, gv, (double)sagn[1][k][threadIdx.x]);
+        gp = gp * pk;
+    }
+    double *Go = gout + ((size_t)b * ngm + grp) * 2 * MP + threadIdx.x;
+    Go[0] = gp;
+    Go[MP] = gv;
+}
+
+// ---------------------------------------------------------------------------------------
 // Reverse fix-up: lam from the carry (lam_{s1} of the chunk), walked down the chunk,
 // optionally written, with the gradient partial sums of the chain at the forced inputs
 // z~_s of the same trajectory (the ReLU row of every step through LDS):
@@ -523,6 +822,35 @@ int launch_qdeer_scan_fwd(int B, int T, int M, const float *x, int N, float *z, 
 #undef FX
     }
     DEER_LAUNCH_CHECK("k_qdeer_fixup_fwd");
+    return DEER_OK;
+}
+
+// chunks per block of the fused pass kernel (the chunk count per sequence is a multiple of it,
+// at most QF_MAXG times it)
+int qdeer_pass_group(int M) { return QF_WPB * (64 / q_padded(M)); }
+int qdeer_pass_max_chunks(int M) { return QF_MAXG * qdeer_pass_group(M); }
+
+int launch_qdeer_pass(const PlrnnArgs &a, float *z, float *zalt, const float *Pin, const float *vin, const double *gin,
+                      float *Pout, float *vout, double *gout, int C, int ncs, const FusedCtl &fc, uint32_t *mark,
+                      uint32_t pass_no, hipStream_t st) {
+    const int MP = q_padded(a.M), GS = qdeer_pass_group(a.M);
+    if (a.M < 1 || a.M > 64 || C < 1 || ncs < GS || ncs % GS || ncs > QF_MAXG * GS || (long)C * ncs < a.T ||
+        (long)C * (ncs - GS) >= a.T ||
+        !fc.seq || !fc.nd.pv || !Pin || !vin || !gin || !Pout || !vout || !gout)
+    {
+        set_error("fused quasi-DEER passes need M <= 64, a chunk count per sequence that is a multiple of %d, at "
+                  "most %d, covering T with fewer than %d padding chunks, the control and two aggregate buffers",
+                  GS, QF_MAXG * GS, GS);
+        return DEER_ERR_INVALID_ARG;
+    }
+    KTimer kt("k_qdeer_pass", st);
+    const unsigned grid = (unsigned)((long)a.B * ncs / GS);
+#define QP(MPV)                                                                                                     \
+    hipLaunchKernelGGL((k_qdeer_pass<MPV>), dim3(grid), dim3(64 * QF_WPB), 0, st, a.A, a.W, a.h, a.alpha, a.N, a.x, \
+                       a.z0, z, zalt, a.T, a.M, C, ncs, Pin, vin, gin, Pout, vout, gout, fc, mark, pass_no, a.tw)
+    if (MP == 16) QP(16); else if (MP == 32) QP(32); else QP(64);
+#undef QP
+    DEER_LAUNCH_CHECK("k_qdeer_pass");
     return DEER_OK;
 }
 

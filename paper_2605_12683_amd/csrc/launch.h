@@ -148,6 +148,16 @@ int qdeer_chunk_len(int B, int T, int M);
 int launch_qdeer_update(const PlrnnArgs &a, float *z, float *zalt, const int *zsel, const int *active,
                         const float *gamma, float *rhs, float *coef, float *P, float *v, float *carry,
                         uint32_t *chain_bits, int C, int ncs, hipStream_t st);
+// Fused quasi-DEER passes of the adaptive loop (vanilla PLRNN): one kernel per pass takes the
+// fix-up of the previous update, where fc.nd.pv says the aggregates in (Pin, vin, gin) belong to
+// the current iterate, and the chunk aggregates of the next update, written to (Pout, vout,
+// gout), with the pass-end control.  ncs is a multiple of qdeer_pass_group(M), at most
+// qdeer_pass_max_chunks(M) (padding chunks past T are empty).  Block 0 writes pass_no to *mark as it starts.
+int qdeer_pass_group(int M);
+int qdeer_pass_max_chunks(int M);
+int launch_qdeer_pass(const PlrnnArgs &a, float *z, float *zalt, const float *Pin, const float *vin, const double *gin,
+                      float *Pout, float *vout, double *gout, int C, int ncs, const FusedCtl &fc, uint32_t *mark,
+                      uint32_t pass_no, hipStream_t st);
 int launch_qdeer_adjoint(const PlrnnArgs &a, const float *g, float seed_scale, const float *z, float *coef, float *P,
                          float *v, float *carry, float *lam, float *gpart, int C, int ncs, hipStream_t st);
 // the model-independent parts: the forward scan + fix-up from (rhs = r, coef), and the reverse

@@ -5,6 +5,8 @@ Tolerance 1e-4 normwise relative for float32 states, adjoints and gradients.  Ne
 iterates are compared where the ReLU decisions of both sides cannot differ: the first update
 from the teacher states, and one update from an iterate given to both; converged solves are
 compared with the sequential rollout (the zero of the residual, independent of the path)."""
+import os
+
 import numpy as np
 import pytest
 
@@ -95,6 +97,40 @@ def test_quasi_adjoint_and_gradients(M, N, B, T, user_g):
     out2 = D.deer_adjoint_quasi(m, c.x, z32, c.alpha, N, g=g, want_lam=False)
     for k, v in out2["grads"].items():
         assert rel_inf(v.cpu().numpy(), gr[k]) < TOL, k
+
+
+@pytest.mark.parametrize("M,N,B,T,alpha,T_w,bound", [(16, 3, 4, 4096, 0.2, 0, 0.0), (8, 2, 3, 2049, 0.2, 0, 0.0),
+                                                     (24, 24, 2, 1500, 0.1, 300, 0.0), (33, 8, 2, 700, 0.2, 0, 0.05),
+                                                     (64, 64, 2, 2050, 0.05, 0, 0.0), (3, 3, 1, 5, 0.1, 0, 0.0),
+                                                     (16, 3, 2, 500, 0.2, 100, 0.05), (50, 7, 5, 333, 0.2, 40, 0.0)])
+def test_quasi_fused_and_separate_passes_agree(M, N, B, T, alpha, T_w, bound):
+    """The adaptive loop's quasi-DEER pass in one kernel (fix-up of an update, chunk aggregates
+    of the next, pass-end control; chunk counts padded to whole groups) and in separate kernels
+    (DEER_QUASI_FUSED=0): both land on the rollout, in the oracle's number of quasi-Newton
+    updates up to one; ragged and padding chunks, several groups per sequence, all three lane
+    widths, latent warm-up and forced rejections (damped coefficients)."""
+    c = _case(M, N, B, T, alpha, 360 + M + T)
+    m = oracle_model(c)
+    ref = O.rollout(m, c.x, alpha, N, T_w=T_w)
+    want = None
+    if bound == 0.0:
+        want = O.newton(m, c.x, alpha, N, tol=1e-5, max_iter=T + 2, T_w=T_w, quasi=True)["iters"].tolist()
+    its = {}
+    try:
+        for fuse in ("1", "0"):
+            os.environ["DEER_QUASI_FUSED"] = fuse
+            say("deer_solve_quasi fused" if fuse == "1" else "deer_solve_quasi separate", M, N, B, T, alpha, T_w, bound)
+            res = D.deer_solve_quasi(m, c.x, alpha, N, tol=1e-5, max_iter=T + 2, step_bound=bound, T_w=T_w)
+            assert res["status"] == 0, (fuse, res)
+            assert rel_inf(res["z"].cpu().numpy(), ref) < TOL, fuse
+            assert all(n < 1e-5 for n in res["norms"]), fuse
+            its[fuse] = res["iters"]
+    finally:
+        os.environ.pop("DEER_QUASI_FUSED", None)
+    print(f"[gpu-case] quasi updates fused {its['1']} separate {its['0']} oracle {want}", flush=True)
+    assert max(abs(a - b) for a, b in zip(its["1"], its["0"])) <= 1
+    if want is not None:
+        assert max(abs(a - b) for a, b in zip(its["1"], want)) <= 1, (its["1"], want)
 
 
 def test_quasi_workload2_full_size():

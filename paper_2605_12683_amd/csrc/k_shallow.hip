@@ -428,19 +428,36 @@ __global__ __launch_bounds__(SHG_THREADS) void k_grads_shplrnn(const ShArgs a, c
 }
 
 // float64 sum over nrows partial rows of length width, then scattered to the outputs
-__global__ void k_reduce_rows(const float *__restrict__ part, int nrows, int width, int M, int L,
-                              float *__restrict__ dW1, float *__restrict__ dW2, float *__restrict__ dh2,
-                              float *__restrict__ dA, float *__restrict__ dh1) {
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= width) return;
-    double s0 = 0.0, s1 = 0.0;
-    int r = 0;
-    for (; r + 1 < nrows; r += 2) {
-        s0 += (double)part[(size_t)r * width + e];
-        s1 += (double)part[(size_t)(r + 1) * width + e];
+// Column sums of part[nrows][width] in float64.  Block = 64 columns x RR_G row groups: thread
+// (g, column) adds rows g, g + RR_G, ... (8 loads issued before their adds), then the row groups
+// are added through LDS in a fixed order, so the sums do not depend on the launch.
+constexpr int RR_G = 16;
+
+__global__ __launch_bounds__(64 * RR_G) void k_reduce_rows(const float *__restrict__ part, int nrows, int width, int M,
+                                                           int L, float *__restrict__ dW1, float *__restrict__ dW2,
+                                                           float *__restrict__ dh2, float *__restrict__ dA,
+                                                           float *__restrict__ dh1) {
+    __shared__ double red[RR_G][64];
+    const int col = threadIdx.x & 63, g = threadIdx.x >> 6;
+    const int e = blockIdx.x * 64 + col;
+    const bool ok = e < width;
+    double s = 0.0;
+    for (int r0 = g; r0 < nrows; r0 += 8 * RR_G) {
+        float v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int r = r0 + k * RR_G;
+            v[k] = (ok && r < nrows) ? part[(size_t)r * width + e] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) s += (double)v[k];
     }
-    if (r < nrows) s0 += (double)part[(size_t)r * width + e];
-    const float v = (float)(s0 + s1);
+    red[g][col] = s;
+    __syncthreads();
+    if (g != 0 || !ok) return;
+    double t = red[0][col];
+    for (int k = 1; k < RR_G; ++k) t += red[k][col];
+    const float v = (float)t;
     const int ML = M * L;
     if (e < ML) {
         if (dW1) dW1[e] = v;
@@ -542,8 +559,8 @@ int launch_grads_shplrnn(const ShArgs &a, const float *z, const float *lam, cons
     const int width = 2 * a.M * a.L + a.L + 2 * a.M;
     {
         KTimer kt("k_reduce_rows", st);
-        hipLaunchKernelGGL(k_reduce_rows, dim3((width + 255) / 256), dim3(256), 0, st, part, nb, width, a.M, a.L, gr->W,
-                           gr->W2, gr->h2, gr->A, gr->h);
+        hipLaunchKernelGGL(k_reduce_rows, dim3((width + 63) / 64), dim3(64 * RR_G), 0, st, part, nb, width, a.M, a.L,
+                           gr->W, gr->W2, gr->h2, gr->A, gr->h);
         DEER_LAUNCH_CHECK("k_reduce_rows");
     }
     return DEER_OK;

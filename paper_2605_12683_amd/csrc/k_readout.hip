@@ -266,7 +266,7 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
                 dca[0] += buf[wv][2 * lane][rr];
                 dca[1] += buf[wv][2 * lane + 1][rr];
             }
-#pragma unroll 2
+#pragma unroll
             for (int w2 = 0; w2 < RW; ++w2) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {

@@ -133,6 +133,28 @@ def test_quasi_fused_and_separate_passes_agree(M, N, B, T, alpha, T_w, bound):
         assert max(abs(a - b) for a, b in zip(its["1"], want)) <= 1, (its["1"], want)
 
 
+@pytest.mark.parametrize("fuse", ["1", "0"])
+def test_quasi_nonfinite_and_not_converged(fuse):
+    """A NaN input ends its sequence as non-finite after the damped retries, and an update cap
+    of one leaves every sequence unconverged after one update, in the one-kernel pass and in
+    the separate kernels."""
+    c = _case(8, 3, 2, 200, 0.2, 17)
+    m = oracle_model(c)
+    x = c.x.copy()
+    x[1, 50, 0] = np.nan
+    try:
+        os.environ["DEER_QUASI_FUSED"] = fuse
+        say("deer_solve_quasi NaN input", fuse)
+        res = D.deer_solve_quasi(m, x, 0.2, 3, tol=1e-5, check=False)
+        assert res["status"] == 3                      # DEER_ERR_NONFINITE
+        say("deer_solve_quasi max_iter=1", fuse)
+        res = D.deer_solve_quasi(m, c.x, 0.2, 3, tol=1e-5, max_iter=1, check=False)
+        assert res["status"] == 2                      # DEER_ERR_NOT_CONVERGED
+        assert res["iters"] == [1, 1]
+    finally:
+        os.environ.pop("DEER_QUASI_FUSED", None)
+
+
 def test_quasi_workload2_full_size():
     """The M = 16 workload (16 Lorenz-63 sequences of 16384 steps, alpha = 0.2, tolerance
     1e-5) with quasi-DEER: the solve lands on the rollout and the adjoint and gradients at

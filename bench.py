@@ -141,6 +141,9 @@ def kernel_work(c, steps, updates):
         out["k_qdeer_chunk"] = ("hbm", fwd * 8 * M + adj * (4 * M + 8 * N))
         out["k_qdeer_fixup_fwd"] = ("hbm", fwd * 16 * M)
         out["k_qdeer_fixup_rev"] = ("hbm", adj * (8 * M + 4 * N))
+        # the adaptive loop's one-kernel quasi pass: z and x read, the next iterate written (the
+        # residual is formed again from them, the chunk aggregates are a few floats per chunk)
+        out["k_qdeer_pass"] = ("hbm", fwd * (8 * M + 4 * N))
         if M <= 16:
             # the register-tiled fix-ups form the residual and the masks again from z and x:
             # forward z, x read and the next iterate written; reverse z, x read (the training

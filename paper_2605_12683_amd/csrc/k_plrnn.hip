@@ -3342,26 +3342,39 @@ __global__ __launch_bounds__(64) void k_fixup_rev_plrnn(const float *__restrict_
     }
 }
 
-// sum the per-chunk partials in float64 in two stages: blocks over (slice of the chains, 256
-// consecutive entries of [MP][MP + 2]), each thread adding its entry over the slice's chains
-// with 8 loads in flight; then the slices
+// sum the per-chunk partials in float64 in two stages: blocks over (slice of the chains, 64
+// consecutive entries of [MP][MP + 2]), the four waves of a block taking every fourth chain of
+// the slice with 8 loads in flight and their sums added through LDS in a fixed order; then the
+// slices
 constexpr int GP_SLICES = 64;
 
 __global__ __launch_bounds__(256) void k_reduce_gpart1(const float *__restrict__ gpart, int nchains, int n,
                                                        double *__restrict__ part2) {
+    __shared__ double red[4][64];
     const int sl = blockIdx.x;
     const int c0 = (int)((long)nchains * sl / GP_SLICES), c1 = (int)((long)nchains * (sl + 1) / GP_SLICES);
-    const int e = blockIdx.y * 256 + threadIdx.x;
-    if (e >= n) return;
-    double s[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int ch0 = c0; ch0 < c1; ch0 += 8) {
+    const int cg = threadIdx.x >> 6;
+    const int e = blockIdx.y * 64 + (threadIdx.x & 63);
+    const bool ok = e < n;
+    double s0 = 0.0, s1 = 0.0;
+    for (int ch0 = c0 + cg; ch0 < c1; ch0 += 32) {
         float v[8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) v[k] = ch0 + k < c1 ? gpart[(size_t)(ch0 + k) * n + e] : 0.f;
+        for (int k = 0; k < 8; ++k) {
+            const int ch = ch0 + 4 * k;
+            v[k] = (ok && ch < c1) ? gpart[(size_t)ch * n + e] : 0.f;
+        }
 #pragma unroll
-        for (int k = 0; k < 8; ++k) s[k & 3] += (double)v[k];
+        for (int k = 0; k < 8; k += 2) {
+            s0 += (double)v[k];
+            s1 += (double)v[k + 1];
+        }
     }
-    part2[(size_t)sl * n + e] = (s[0] + s[1]) + (s[2] + s[3]);
+    red[cg][threadIdx.x & 63] = s0 + s1;
+    __syncthreads();
+    if (cg != 0 || !ok) return;
+    const int l = threadIdx.x & 63;
+    part2[(size_t)sl * n + e] = (red[0][l] + red[1][l]) + (red[2][l] + red[3][l]);
 }
 
 __global__ __launch_bounds__(256) void k_reduce_gpart2(const double *__restrict__ part2, int MP, int M,
@@ -3802,7 +3815,7 @@ int launch_reduce_gpart(const float *gpart, int nchains, int MP, int M, float *d
     const int n = MP * (MP + 2);
     {
         KTimer _kt("k_reduce_gpart", st);
-        hipLaunchKernelGGL(k_reduce_gpart1, dim3(GP_SLICES, (n + 255) / 256), dim3(256), 0, st, gpart, nchains, n, part2);
+        hipLaunchKernelGGL(k_reduce_gpart1, dim3(GP_SLICES, (n + 63) / 64), dim3(256), 0, st, gpart, nchains, n, part2);
         hipLaunchKernelGGL(k_reduce_gpart2, dim3((n + 255) / 256), dim3(256), 0, st, (const double *)part2, MP, M, dA,
                            dW, dh);
     }

@@ -329,8 +329,9 @@ __global__ __launch_bounds__(64) void k_qdeer_fixup_fwd(const float *__restrict_
 //   1. when the sequence's aggregates of the previous kernel belong to its current iterate
 //      (nd.pv == pass_no): the chunk's carry, walked in float64 over the group maps of the
 //      groups before it and the chunk aggregates before it in its group, then the fix-up
-//      Delta_s = coef_s Delta_{s-1} - r_s with r and coef formed again from z (the same
-//      operations as the separate kernels), z + Delta written to the other iterate buffer;
+//      Delta_s = coef_s Delta_{s-1} - r_s with r and coef formed again from z and x by the
+//      operations step 2 of the previous kernel formed them with (so they are the values its
+//      aggregates hold), z + Delta written to the other iterate buffer;
 //   2. the chunk aggregates of the next update at the new iterate (or at the current one when
 //      step 1 did not run): prod coef and the local solution from zero, with the damping that
 //      an accepted update leads to, and the group map of the block (float64);

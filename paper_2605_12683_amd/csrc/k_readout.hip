@@ -17,7 +17,7 @@
 //          of all eight tiles (dS and H through LDS), so a wave keeps 16 accumulator floats per
 //          lane instead of the whole 128 x 64 dWa, and two waves fit on every SIMD
 // The k ordering of GEMM1 is permuted (k-step (jj, q) uses channel 16 jj + 4 g + q in lane group
-// g) so that four k-steps read one 16-byte LDS vector for both operands.
+// g) so that four k-steps read one 16-byte LDS vector of Wa.
 #include "common.h"
 #include "launch.h"
 
@@ -28,8 +28,12 @@ constexpr int RH = 128;          // hidden units (padded)
 constexpr int RM = 64;           // state channels (padded)
 constexpr int RNO = 4;           // outputs (padded)
 constexpr int RW = 8;            // waves per block (one per 16 hidden units in GEMM3)
-constexpr int WS = RM + 4;       // LDS row stride of Wa and of the H tile (16-byte aligned rows)
+constexpr int WS = RM + 4;       // LDS row stride of Wa (16-byte aligned rows)
 constexpr int BS = 17;           // LDS row stride of the [hidden][row] tile
+// The H tile sits channel-major in LDS, [channel][row] with a row stride of 20 floats: GEMM1
+// reads H[row c][channel 16 jj + 4 g + q] and GEMM3 H[row 4 j + g][channel 16 q + c], and with
+// 20 = 4 (mod 16) both patterns put the 64 lanes of a read on 64 distinct banks
+constexpr int HTS = 20;
 constexpr int RPS = RH * RM + RNO * RH + RH + RNO + 1;   // partial floats per wave
 constexpr int RPS_PAD = (RPS + 63) & ~63;
 }  // namespace
@@ -43,7 +47,7 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
     __shared__ float wb[RNO][RH];
     __shared__ float cas[RH];
     __shared__ float cbs[RNO];
-    __shared__ __align__(16) float hti[RW][16][WS];
+    __shared__ float hti[RW][RM][HTS];
     __shared__ float buf[GRADS ? RW : 1][RH][BS];
     __shared__ float dyv[GRADS ? RW : 1][16][RNO];
     __shared__ float lsw[RW];
@@ -96,7 +100,7 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
         const long tile = base + wv;
         const long r0 = tile * 16;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) hti[wv][i][lane] = hv[i];
+        for (int i = 0; i < 16; ++i) hti[wv][lane][i] = hv[i];
         load_tile(tile + (long)gridDim.x * RW);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
@@ -109,7 +113,11 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
         for (int n = 0; n < 8; ++n) acc1[n] = (v4f){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
-            const float4 bq = *reinterpret_cast<const float4 *>(&hti[wv][c][16 * jj + 4 * g]);
+            float4 bq;
+            bq.x = hti[wv][16 * jj + 4 * g + 0][c];
+            bq.y = hti[wv][16 * jj + 4 * g + 1][c];
+            bq.z = hti[wv][16 * jj + 4 * g + 2][c];
+            bq.w = hti[wv][16 * jj + 4 * g + 3][c];
             float4 aq[8];
 #pragma unroll
             for (int n = 0; n < 8; ++n) aq[n] = *reinterpret_cast<const float4 *>(&wa[16 * n + c][16 * jj + 4 * g]);
@@ -272,7 +280,7 @@ __global__ __launch_bounds__(RW * 64) void k_readout(const RoArgs ra, const floa
                 for (int j = 0; j < 4; ++j) {
                     const float bv = buf[w2][16 * wv + c][4 * j + g];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) acc3[q] = mfma16x16x4(hti[w2][4 * j + g][16 * q + c], bv, acc3[q]);
+                    for (int q = 0; q < 4; ++q) acc3[q] = mfma16x16x4(hti[w2][16 * q + c][4 * j + g], bv, acc3[q]);
                 }
             }
             // the next round overwrites hti and buf: every wave is past its reads

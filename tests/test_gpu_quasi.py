@@ -102,7 +102,8 @@ def test_quasi_adjoint_and_gradients(M, N, B, T, user_g):
 @pytest.mark.parametrize("M,N,B,T,alpha,T_w,bound", [(16, 3, 4, 4096, 0.2, 0, 0.0), (8, 2, 3, 2049, 0.2, 0, 0.0),
                                                      (24, 24, 2, 1500, 0.1, 300, 0.0), (33, 8, 2, 700, 0.2, 0, 0.05),
                                                      (64, 64, 2, 2050, 0.05, 0, 0.0), (3, 3, 1, 5, 0.1, 0, 0.0),
-                                                     (16, 3, 2, 500, 0.2, 100, 0.05), (50, 7, 5, 333, 0.2, 40, 0.0)])
+                                                     (16, 3, 2, 500, 0.2, 100, 0.05), (50, 7, 5, 333, 0.2, 40, 0.0),
+                                                     (1, 1, 1, 1, 0.2, 0, 0.0), (4, 2, 3, 2, 0.2, 1, 0.0)])
 def test_quasi_fused_and_separate_passes_agree(M, N, B, T, alpha, T_w, bound):
     """The adaptive loop's quasi-DEER pass in one kernel (fix-up of an update, chunk aggregates
     of the next, pass-end control; chunk counts padded to whole groups) and in separate kernels

@@ -237,12 +237,17 @@ static int choose_chunk(int B, int T, int MP, bool sh_fused = false) {
     }
     const long target_chains = (MP == 64 || sh_fused) ? 8192L : 2048L * (64 / MP);
     long C = (total + target_chains - 1) / target_chains;
-    if (C < 16) C = 16;
+    // at least 16 steps per chunk (8 on the shallow path without a stored Jacobian, whose chunk
+    // steps are long chains of dependent products: for short sequences a chunk's serial walk,
+    // not the carry pass, sets a pass's time)
+    const long minStep = sh_fused ? 8 : 16;
+    if (C < minStep) C = minStep;
     const long maxc = MP <= 32 ? 1024 : 512;
     const long minC = (T + maxc - 1) / maxc;
     if (C < minC) C = minC;
-    // M <= 16: whole 16-step tiles (the register-tiled kernels run a partial tile step by step)
-    if (MP == 16) C = (C + 15) / 16 * 16;
+    // vanilla M <= 16: whole 16-step tiles (the register-tiled kernels run a partial tile step by
+    // step)
+    if (MP == 16 && !sh_fused) C = (C + 15) / 16 * 16;
     if (C > T) C = T;
     return (int)C;
 }
@@ -691,7 +696,8 @@ static int newton_loop(const deer_solve_opts *o, int B, size_t seq_elems, int nc
     };
     bool stopped = false;
     if (ctl.fused) {
-        // Short passes (the fused M <= 16 path).  The forward pass of pass p marks its start,
+        // Passes whose last kernel takes the pass-end control (the vanilla M <= 16 and shallow
+        // fix-ups, the one-kernel passes).  The first kernel of pass p marks its start,
         // when every earlier pass, and so the decisions of pass p - 1, is complete.  The host
         // keeps one pass queued ahead: once pass p has started it reads the flags as of pass
         // p - 1 and queues pass p + 1 (a whole pass of time to do so), so the device does not
@@ -909,11 +915,21 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
     std::vector<float> norm(B, NAN);
     bool nonfinite = false;
     const DenseWs &d = w.d;
-    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *,
-                      uint32_t) -> int {
+    // adaptive loop on the path without a stored Jacobian: the fix-up takes the pass-end control
+    // and the residual kernel marks each pass's start, so passes are queued one ahead with no
+    // control kernel and no host wait per pass
+    NewtonCtl ctl = w.ctl;
+    ctl.fused = fused && sh_res_mfma() && o->fixed_iters <= 0;
+    if (ctl.fused) {
+        uint32_t *mark_unused = nullptr;
+        if ((rc = host_block(B, ctl.nd, &mark_unused))) return rc;
+    }
+    const FusedCtl fc{ctl.nd, ctl.seq, o->tol, o->step_bound == 0.f ? kDefaultStepBound : o->step_bound, kDamp};
+    auto update = [&](const int *dact, const float *gam, const int *zsel, float *zb, float *za, uint32_t *mark,
+                      uint32_t pass_no) -> int {
         int r;
         if (fused && sh_res_mfma()) {
-            if ((r = launch_resjac_shmfma(a, zb, za, zsel, w.r, w.masks, dact, st))) return r;
+            if ((r = launch_resjac_shmfma(a, zb, za, zsel, w.r, w.masks, dact, st, mark, pass_no))) return r;
         } else if ((r = launch_resjac_shplrnn(a, zb, za, zsel, nullptr, w.r, w.masks, dact, st))) {
             return r;
         }
@@ -922,7 +938,7 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
                 return r;
             if ((r = launch_carry(d.MP, false, d.P, d.v, d.carry, dact, nullptr, B, d.ncs, d.gws, st))) return r;
             return launch_fixup_shjvp(false, a, w.masks, w.r, -1.f, gam, d.carry, zb, za, zsel, w.ctl.chain_bits, dact,
-                                      d.C, d.ncs, st);
+                                      d.C, d.ncs, st, (ctl.fused && dact) ? &fc : nullptr);
         }
         if ((r = jacform_sh(a, w.masks, w.J, dact, gam, st))) return r;
         if ((r = launch_chunk_product_dense(false, B, T, m->M, w.J, w.r, -1.f, d.P, d.v, dact, d.C, d.ncs, st))) return r;
@@ -930,7 +946,7 @@ static int solve_shplrnn(const deer_model *m, const deer_forcing *f, const deer_
         return launch_fixup_dense(0, B, T, m->M, w.J, w.r, -1.f, d.carry, zb, za, zsel, w.ctl.chain_bits, dact, d.C,
                                   d.ncs, st);
     };
-    if ((rc = newton_loop(o, B, (size_t)T * m->M, d.ncs, w.ctl, z, update, it, norm, nonfinite, act, st))) return rc;
+    if ((rc = newton_loop(o, B, (size_t)T * m->M, d.ncs, ctl, z, update, it, norm, nonfinite, act, st))) return rc;
     if (masks) {
         if ((rc = launch_resjac_shplrnn(a, z, nullptr, nullptr, nullptr, nullptr, masks, nullptr, st))) return rc;
     }

@@ -17,6 +17,7 @@
 // Per step this replaces 4 M^2 bytes written and read twice by 4 L / 8 bytes of masks.
 #include "common.h"
 #include "launch.h"
+#include "newton_ctl.h"
 
 namespace deer {
 
@@ -411,7 +412,7 @@ __global__ __launch_bounds__(256) void k_fixup_shjvp(const ShArgs a, const uint3
                                                      const float *__restrict__ gamma,
                                                      const float *__restrict__ carry_in, float *zbuf, float *outbuf,
                                                      const int *__restrict__ zsel, uint32_t *__restrict__ chain_bits,
-                                                     const int *__restrict__ active, int C, int ncs) {
+                                                     const int *__restrict__ active, int C, int ncs, FusedCtl fc) {
     constexpr int NI = MP / 16, NS = MP / 4;
     __shared__ v4f red[2][4][NI][64];
     const int tid = threadIdx.x, wv = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4,
@@ -601,14 +602,43 @@ __global__ __launch_bounds__(256) void k_fixup_shjvp(const ShArgs a, const uint3
         mx[wv][c][1] = zmax;
     }
     lds_barrier();
-    if (wv == 0 && g == 0 && ok) {   // reduced per sequence by the pass-end control
+    if (wv != 0) return;
+    if (g == 0 && ok) {
 #pragma unroll
         for (int w = 1; w < 4; ++w) {
             emax = emax > mx[w][c][0] ? emax : mx[w][c][0];
             zmax = zmax > mx[w][c][1] ? zmax : mx[w][c][1];
         }
-        chain_bits[id] = emax;
-        chain_bits[(size_t)nchains + id] = zmax;
+        if (!fc.seq) {   // reduced per sequence by the pass-end control
+            chain_bits[id] = emax;
+            chain_bits[(size_t)nchains + id] = zmax;
+        }
+    }
+    if (!fc.seq) return;
+    // fused pass-end control: lane 0 gathers the 16 chains' maxima and arrives once per
+    // sequence they belong to (chains of a sequence that is not running do not arrive)
+    uint32_t em[16], zm[16];
+    bool okc[16];
+#pragma unroll
+    for (int n = 0; n < 16; ++n) {
+        em[n] = (uint32_t)__shfl((int)emax, n, 64);
+        zm[n] = (uint32_t)__shfl((int)zmax, n, 64);
+        okc[n] = __shfl((int)ok, n, 64) != 0;
+    }
+    if (lane != 0) return;
+    const int chain0 = blockIdx.x * 16;
+    for (int n = 0; n < 16; ++n) {
+        if (!okc[n]) continue;
+        const int bn = (chain0 + n) / ncs;
+        if (n > 0 && okc[n - 1] && (chain0 + n - 1) / ncs == bn) continue;   // counted with its first chain
+        uint32_t E = 0u, Z = 0u;
+        int cnt = 0;
+        for (int m2 = n; m2 < 16 && okc[m2] && (chain0 + m2) / ncs == bn; ++m2) {
+            E = E > em[m2] ? E : em[m2];
+            Z = Z > zm[m2] ? Z : zm[m2];
+            ++cnt;
+        }
+        seq_arrive(fc, bn, cnt, ncs, E, Z);
     }
 }
 
@@ -635,9 +665,12 @@ template <int MP>
 __global__ __launch_bounds__(256) void k_resjac_shmfma(const ShArgs a, const float *zbuf, const float *zalt,
                                                        const int *__restrict__ zsel, float *__restrict__ r_out,
                                                        uint32_t *__restrict__ masks, const int *__restrict__ active,
-                                                       int LP) {
+                                                       int LP, uint32_t *mark, uint32_t pass_no) {
     constexpr int NI = MP / 16, MQ = MP + 4;
     extern __shared__ __align__(16) float smem[];
+    // the pass's first kernel: block 0 marks its start (every earlier pass is complete)
+    if (mark && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(mark, pass_no, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     const int M = a.M, L = a.L, T = a.T, N = a.N, LQ = LP + 4;
     float *w2s = smem;             // [LP][MQ]
     float *w1s = w2s + LP * MQ;    // [MP][LQ]
@@ -794,7 +827,7 @@ __global__ __launch_bounds__(256) void k_resjac_shmfma(const ShArgs a, const flo
 }
 
 int launch_resjac_shmfma(const ShArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
-                         uint32_t *masks, const int *active, hipStream_t st) {
+                         uint32_t *masks, const int *active, hipStream_t st, uint32_t *mark, uint32_t pass_no) {
     const int MP = padded_dim(a.M);
     if (!shfused_supported(a.M, a.L) || a.zt) return DEER_ERR_INVALID_ARG;
     const size_t lds = shf_resjac_lds(a.M, a.L);
@@ -806,7 +839,8 @@ int launch_resjac_shmfma(const ShArgs &a, const float *z, const float *zalt, con
     const int LP = shf_LP(a.L);
     KTimer kt("k_resjac_shmfma", st);
 #define RJM(MPV) \
-    hipLaunchKernelGGL((k_resjac_shmfma<MPV>), dim3(grid), dim3(256), lds, st, a, z, zalt, zsel, r, masks, active, LP)
+    hipLaunchKernelGGL((k_resjac_shmfma<MPV>), dim3(grid), dim3(256), lds, st, a, z, zalt, zsel, r, masks, active, LP, \
+                       mark, pass_no)
     if (MP == 16) RJM(16); else if (MP == 32) RJM(32); else RJM(64);
 #undef RJM
     DEER_LAUNCH_CHECK("k_resjac_shmfma");
@@ -842,16 +876,17 @@ int launch_chunk_product_shfused(bool rev, const ShArgs &a, const uint32_t *mask
 
 int launch_fixup_shjvp(bool rev, const ShArgs &a, const uint32_t *masks, const float *rhs, float rhs_sign,
                        const float *gamma, const float *carry_in, float *z, float *out, const int *zsel,
-                       uint32_t *chain_bits, const int *active, int C, int ncs, hipStream_t st) {
+                       uint32_t *chain_bits, const int *active, int C, int ncs, hipStream_t st, const FusedCtl *fc) {
     const int MP = padded_dim(a.M);
-    if (!shfused_supported(a.M, a.L)) return DEER_ERR_INVALID_ARG;
+    if (!shfused_supported(a.M, a.L) || (fc && (rev || !active))) return DEER_ERR_INVALID_ARG;
+    const FusedCtl fcv = fc ? *fc : FusedCtl{};
     const int nch = a.B * ncs;
     const int grid = (nch + 15) / 16;
     const int nlw = shf_nlw(a.L);
     KTimer kt(rev ? "k_fixup_shjvp_rev" : "k_fixup_shjvp", st);
 #define FXJ(MPV, NL, RV)                                                                                         \
     hipLaunchKernelGGL((k_fixup_shjvp<MPV, NL, RV>), dim3(grid), dim3(256), 0, st, a, masks, rhs, rhs_sign, gamma, \
-                       carry_in, z, out, zsel, chain_bits, active, C, ncs)
+                       carry_in, z, out, zsel, chain_bits, active, C, ncs, fcv)
     // shfused_supported bounds NLW * MP / 2 (the A fragments per lane) by 64
 #define FXJ_ALL(RV)                                                                                                  \
     if (MP == 16) {                                                                                                  \

@@ -4,7 +4,7 @@
 
 namespace deer {
 
-struct FusedCtl;   // pass-end control fused into the M <= 16 fix-up (defined below)
+struct FusedCtl;   // pass-end control fused into a pass kernel (defined below)
 
 struct PlrnnArgs {
     const float *A, *W, *h;
@@ -204,15 +204,19 @@ int launch_grads_big(const ShArgs &a, const float *z, const float *lam, const ui
 // shallow PLRNN Newton update without a stored Jacobian (masks + W1, W2 only)
 bool shfused_supported(int M, int L);
 size_t shfused_product_lds(int M, int L);
+// mark: with the adaptive loop's one-pass-ahead queueing, block 0 writes pass_no to it as it starts
 int launch_resjac_shmfma(const ShArgs &a, const float *z, const float *zalt, const int *zsel, float *r,
-                         uint32_t *masks, const int *active, hipStream_t st);
+                         uint32_t *masks, const int *active, hipStream_t st, uint32_t *mark = nullptr,
+                         uint32_t pass_no = 0u);
 // rev: the adjoint's reverse recursion (gamma and active must be null; the fix-up writes y to out)
 int launch_chunk_product_shfused(bool rev, const ShArgs &a, const uint32_t *masks, const float *rhs,
                                  float rhs_sign, const float *gamma, float *P, float *v, const int *active, int C,
                                  int ncs, hipStream_t st);
+// fc (forward, adaptive loop only): the fix-up takes the pass-end control itself (no chain_bits)
 int launch_fixup_shjvp(bool rev, const ShArgs &a, const uint32_t *masks, const float *rhs, float rhs_sign,
                        const float *gamma, const float *carry_in, float *z, float *out, const int *zsel,
-                       uint32_t *chain_bits, const int *active, int C, int ncs, hipStream_t st);
+                       uint32_t *chain_bits, const int *active, int C, int ncs, hipStream_t st,
+                       const FusedCtl *fc = nullptr);
 size_t sh_resjac_lds(int M, int L);
 size_t sh_jacform_lds(int M, int L);
 size_t sh_grads_part_floats(int M, int L, int *nblocks);

@@ -33,11 +33,17 @@ __device__ __forceinline__ float eload(const float *__restrict__ Jp, int M, int 
 
 // REV: the product covers steps [s0 + 1, min(s1 + 1, T)) (the reverse chunk map is its
 // transpose) and the local solution runs u_k = E_{k+1}^T u_{k+1} + rhs_k from k = s1 - 1 down.
+// The step's E (128 x 128, zero outside M x M) is staged in LDS by the whole workgroup, the next
+// step's loads in flight while the matrix cores work on this one (double buffer), and every wave
+// reads its A operands there; the forward local solution reads the same tile.
+constexpr int JST = BG + 4;   // LDS row stride of the staged E (16-byte rows, conflict-free reads)
+
 template <bool REV, bool FLIP>
 __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restrict__ J, const float *__restrict__ rhs,
                                                            float rhs_sign, float *__restrict__ Pout,
                                                            float *__restrict__ vout, const int *__restrict__ active,
                                                            int B, int T, int M, int C, int ncs) {
+    __shared__ __align__(16) float js[2][BG][JST];
     __shared__ __align__(16) float ub[2][BG];
     const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
     const int id = blockIdx.x;   // chain
@@ -48,6 +54,29 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
     const int plen = ok ? max(hi - lo, 0) : 0;
     const int ulen = ok ? s1 - s0 : 0;
     const int nsteps = max(plen, ulen);
+    // staging: thread tid takes the 16-byte groups tid + 256 k (k < 16) of the 128 x 128 tile,
+    // row (tid + 256 k) / 32, columns 4 ((tid + 256 k) % 32) .. + 3
+    float4 pre[16];
+    auto stage_load = [&](int t) {
+        const float *Jp = J + ((size_t)b * T + lo + t) * M * M;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            const int e4 = tid + 256 * k, row = e4 >> 5, c4 = (e4 & 31) * 4;
+            if (!FLIP && (M & 3) == 0 && row < M && c4 + 3 < M) {
+                pre[k] = *reinterpret_cast<const float4 *>(Jp + (size_t)row * M + c4);
+            } else {
+                pre[k] = make_float4(eload<FLIP>(Jp, M, row, c4), eload<FLIP>(Jp, M, row, c4 + 1),
+                                     eload<FLIP>(Jp, M, row, c4 + 2), eload<FLIP>(Jp, M, row, c4 + 3));
+            }
+        }
+    };
+    auto stage_store = [&](int buf) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            const int e4 = tid + 256 * k;
+            *reinterpret_cast<float4 *>(&js[buf][e4 >> 5][(e4 & 31) * 4]) = pre[k];
+        }
+    };
     // accumulators: acc[I][Jt][r] = P[16 I + 4 g + r][32 wv + 16 Jt + c]
     v4f acc[8][2];
 #pragma unroll
@@ -59,11 +88,16 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
     // local solution: thread pair (row i = tid / 2, half hh) sums half of the row
     const int ui = tid >> 1, hh = tid & 1;
     if (tid < BG) ub[0][tid] = 0.f;
+    if (plen > 0) {
+        stage_load(0);
+        stage_store(0);
+    }
     __syncthreads();
     int cur = 0;
     for (int t = 0; t < nsteps; ++t) {
+        const bool more = t + 1 < plen;
+        if (more) stage_load(t + 1);   // in flight during this step
         if (t < plen) {
-            const float *Jp = J + ((size_t)b * T + lo + t) * M * M;
             v4f old[8][2];
 #pragma unroll
             for (int I = 0; I < 8; ++I)
@@ -74,51 +108,45 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
                 }
 #pragma unroll
             for (int I = 0; I < 8; ++I) {
-                const int row = 16 * I + c;
-                float a[8][4];
+                float4 a[8];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int k0 = 16 * j + 4 * g;
-                    if (!FLIP && row < M && k0 + 3 < M && (M & 3) == 0) {
-                        const float4 v = *reinterpret_cast<const float4 *>(Jp + (size_t)row * M + k0);
-                        a[j][0] = v.x; a[j][1] = v.y; a[j][2] = v.z; a[j][3] = v.w;
-                    } else {
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) a[j][q] = eload<FLIP>(Jp, M, row, k0 + q);
-                    }
-                }
+                for (int j = 0; j < 8; ++j) a[j] = *reinterpret_cast<const float4 *>(&js[cur][16 * I + c][16 * j + 4 * g]);
 #pragma unroll
                 for (int Jt = 0; Jt < 2; ++Jt) {
                     v4f s = acc[I][Jt];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j)
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) s = mfma16x16x4(a[j][q], old[j][Jt][q], s);
+                    for (int j = 0; j < 8; ++j) {
+                        s = mfma16x16x4(a[j].x, old[j][Jt][0], s);
+                        s = mfma16x16x4(a[j].y, old[j][Jt][1], s);
+                        s = mfma16x16x4(a[j].z, old[j][Jt][2], s);
+                        s = mfma16x16x4(a[j].w, old[j][Jt][3], s);
+                    }
                     acc[I][Jt] = s;
                 }
             }
         }
         if (t < ulen) {
-            // forward: u_s = E_s u_{s-1} + sign rhs_s, s = s0 + t;  reverse: k = s1 - 1 - t,
-            // u_k = E_{k+1}^T u_{k+1} + sign rhs_k (E_T does not exist: the first reverse step
-            // starts from zero)
+            // forward: u_s = E_s u_{s-1} + sign rhs_s, s = s0 + t (E_s is the staged tile);
+            // reverse: k = s1 - 1 - t, u_k = E_{k+1}^T u_{k+1} + sign rhs_k (E_T does not exist:
+            // the first reverse step starts from zero)
             const int k = REV ? s1 - 1 - t : s0 + t;
             const int kj = REV ? k + 1 : k;
             float part = 0.f;
             if (ui < M && (!REV || kj < T)) {
-                const float *Jp = J + ((size_t)b * T + kj) * M * M;
-                for (int q = hh; q < M; q += 2) {
-                    // forward: row ui of E; reverse: column ui of E (row ui of E^T)
-                    const float e = REV ? eload<FLIP>(Jp, M, q, ui) : eload<FLIP>(Jp, M, ui, q);
-                    part = fmaf(e, ub[cur][q], part);
+                if (REV) {
+                    const float *Jp = J + ((size_t)b * T + kj) * M * M;
+                    for (int q = hh; q < M; q += 2) part = fmaf(eload<FLIP>(Jp, M, q, ui), ub[cur][q], part);
+                } else {
+                    for (int q = hh; q < M; q += 2) part = fmaf(js[cur][ui][q], ub[cur][q], part);
                 }
             }
             part += __shfl_xor(part, 1, 64);
             if (hh == 0 && ui < BG)
                 ub[cur ^ 1][ui] = ui < M ? fmaf(rhs_sign, rhs[((size_t)b * T + k) * M + ui], part) : 0.f;
-            __syncthreads();
-            cur ^= 1;
         }
+        if (more) stage_store(cur ^ 1);   // that buffer's reads ended at the previous barrier
+        __syncthreads();
+        cur ^= 1;
     }
     if (!ok) return;
     float *P = Pout + (size_t)id * BG * BG;

@@ -184,65 +184,144 @@ __global__ __launch_bounds__(BG) void k_carry_big(const float *__restrict__ P, c
 }
 
 // MODE 0: Newton fix-up (next iterate = current + Delta, per-chain max |Delta| and max |z|);
-// MODE 1: forward bare scan; MODE 2: reverse (y_k = E_{k+1}^T y_{k+1} + b_k)
+// MODE 1: forward bare scan; MODE 2: reverse (y_k = E_{k+1}^T y_{k+1} + b_k).  256 threads: lane
+// l of wave w forms half hh = l / 32 of row i = 32 w + l % 32 of E y (MODE 2: of E^T y), the two
+// halves added across the wave.  Each step's E is staged in LDS by the block with coalesced
+// loads, the next step's loads (and its right-hand side and iterate) in flight during this step.
+// With a row stride of 129 floats and the second half's walk started 32 entries in, the 64 lanes
+// of a read fall on distinct banks, for rows (MODE 0, 1) and for columns (MODE 2).
+constexpr int FST = BG + 1;
+
 template <int MODE, bool FLIP>
-__global__ __launch_bounds__(BG) void k_fixup_big(const float *__restrict__ J, const float *__restrict__ rhs,
-                                                  float rhs_sign, const float *__restrict__ carry_in, float *zbuf,
-                                                  float *outbuf, const int *__restrict__ zsel,
-                                                  uint32_t *__restrict__ chain_bits, const int *__restrict__ active,
-                                                  int B, int T, int M, int C, int ncs) {
+__global__ __launch_bounds__(256) void k_fixup_big(const float *__restrict__ J, const float *__restrict__ rhs,
+                                                   float rhs_sign, const float *__restrict__ carry_in, float *zbuf,
+                                                   float *outbuf, const int *__restrict__ zsel,
+                                                   uint32_t *__restrict__ chain_bits, const int *__restrict__ active,
+                                                   int B, int T, int M, int C, int ncs) {
+    __shared__ float js[2][BG][FST];
     __shared__ float ys[2][BG];
-    __shared__ uint32_t red[2][BG / 64];
-    const int id = blockIdx.x, i = threadIdx.x;
+    __shared__ uint32_t red[2][4];
+    const int id = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int hh = lane >> 5, i = 32 * w + (lane & 31);
     const int b = id / ncs, cc = id % ncs;
     const bool ok = !active || active[b];
     const int s0 = cc * C, s1 = ok ? min(s0 + C, T) : s0;
+    const int len = s1 - s0;
     const float *zin = MODE == 0 ? cur_iter(zbuf, outbuf, zsel, b) : nullptr;
     float *out = MODE == 0 ? next_iter(zbuf, outbuf, zsel, b) : outbuf;
-    ys[0][i] = (ok && i < M) ? carry_in[(size_t)id * BG + i] : 0.f;
+    const bool own = hh == 0 && i < M;   // the lane that writes row i
+    // step t: k = the row of the output, kj = the matrix (MODE 2: k + 1, none past the end)
+    auto k_of = [&](int t) { return MODE == 2 ? s1 - 1 - t : s0 + t; };
+    // staging: thread tid takes the 16-byte groups tid + 256 q (q < 16), row (tid + 256 q) / 32
+    float4 pre[16];
+    float rpre = 0.f, zpre = 0.f;
+    // row-major E with M % 4 == 0: 16-byte loads through a resource bounded at the matrix's end
+    // (rows past M read zero) with one lane offset (columns past M: an offset outside it)
+    const bool fast = !FLIP && (M & 3) == 0;
+    const uint32_t vlane = ((tid & 31) * 4 + 3 < M) ? 4u * ((uint32_t)(tid >> 5) * M + (tid & 31) * 4) : kOffLane;
+    auto stage_load = [&](int t) {
+        const int k = k_of(t), kj = MODE == 2 ? k + 1 : k;
+        const bool has = kj < T;
+        const float *Jp = J + ((size_t)b * T + (has ? kj : 0)) * M * M;
+        if (fast) {
+            const auto rs = bounded_rsrc(Jp, has ? (uint32_t)M * M * 4u : 0u);
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                pre[q] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)vlane, q * 32 * M, 0));
+        } else {
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int e4 = tid + 256 * q, row = e4 >> 5, c4 = (e4 & 31) * 4;
+                pre[q] = !has ? make_float4(0.f, 0.f, 0.f, 0.f)
+                              : make_float4(eload<FLIP>(Jp, M, row, c4), eload<FLIP>(Jp, M, row, c4 + 1),
+                                            eload<FLIP>(Jp, M, row, c4 + 2), eload<FLIP>(Jp, M, row, c4 + 3));
+            }
+        }
+        if (own) {
+            const size_t e = ((size_t)b * T + k) * M + i;
+            rpre = rhs[e];
+            if (MODE == 0) zpre = zin[e];
+        }
+    };
+    auto stage_store = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int e4 = tid + 256 * q, row = e4 >> 5, c4 = (e4 & 31) * 4;
+            js[buf][row][c4] = pre[q].x;
+            js[buf][row][c4 + 1] = pre[q].y;
+            js[buf][row][c4 + 2] = pre[q].z;
+            js[buf][row][c4 + 3] = pre[q].w;
+        }
+    };
+    if (tid < BG) ys[0][tid] = (ok && tid < M) ? carry_in[(size_t)id * BG + tid] : 0.f;
+    float rc = 0.f, zc = 0.f;
+    if (len > 0) {
+        stage_load(0);
+        stage_store(0);
+        rc = rpre;
+        zc = zpre;
+    }
     __syncthreads();
     uint32_t emax = 0u, zmax = 0u;
     int cur = 0;
-    for (int t = 0; t < s1 - s0; ++t) {
-        const int k = MODE == 2 ? s1 - 1 - t : s0 + t;
-        const int kj = MODE == 2 ? k + 1 : k;
-        float acc = 0.f;
-        if (i < M && kj < T) {
-            const float *Jp = J + ((size_t)b * T + kj) * M * M;
-            for (int q = 0; q < M; ++q) {
-                const float e = MODE == 2 ? eload<FLIP>(Jp, M, q, i) : eload<FLIP>(Jp, M, i, q);
-                acc = fmaf(e, ys[cur][q], acc);
-            }
+    const int q0 = 64 * hh;
+    for (int t = 0; t < len; ++t) {
+        const int k = k_of(t);
+        const bool more = t + 1 < len;
+        if (more) stage_load(t + 1);   // in flight during this step
+        // half hh of the sum over q in [64 hh, 64 hh + 64), walked from 32 hh on (entries past M
+        // are zero in the staged tile and in ys)
+        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll 4
+        for (int u = 0; u < 64; u += 4) {
+            const int q = q0 + ((u + 32 * hh) & 63);
+            const float e0 = MODE == 2 ? js[cur][q][i] : js[cur][i][q];
+            const float e1 = MODE == 2 ? js[cur][q + 1][i] : js[cur][i][q + 1];
+            const float e2 = MODE == 2 ? js[cur][q + 2][i] : js[cur][i][q + 2];
+            const float e3 = MODE == 2 ? js[cur][q + 3][i] : js[cur][i][q + 3];
+            a0 = fmaf(e0, ys[cur][q], a0);
+            a1 = fmaf(e1, ys[cur][q + 1], a1);
+            a2 = fmaf(e2, ys[cur][q + 2], a2);
+            a3 = fmaf(e3, ys[cur][q + 3], a3);
         }
+        float part = (a0 + a1) + (a2 + a3);
+        part += __shfl_xor(part, 32, 64);
         float y = 0.f;
-        if (i < M) {
+        if (own) {
             const size_t e = ((size_t)b * T + k) * M + i;
-            y = fmaf(rhs_sign, rhs[e], acc);
+            y = fmaf(rhs_sign, rc, part);
             if (MODE == 0) {
-                const float zo = zin[e];
-                out[e] = zo + y;
-                const uint32_t ab = abs_bits(y), zb = abs_bits(zo);
+                out[e] = zc + y;
+                const uint32_t ab = abs_bits(y), zb = abs_bits(zc);
                 emax = emax > ab ? emax : ab;
                 zmax = zmax > zb ? zmax : zb;
             } else {
                 out[e] = y;
             }
         }
-        ys[cur ^ 1][i] = y;
+        if (hh == 0) ys[cur ^ 1][i] = y;
+        if (more) {
+            stage_store(cur ^ 1);   // that buffer's reads ended at the previous barrier
+            rc = rpre;
+            zc = zpre;
+        }
         __syncthreads();
         cur ^= 1;
     }
     if (MODE == 0) {
         emax = wave_max_u32(emax);
         zmax = wave_max_u32(zmax);
-        if ((i & 63) == 0) {
-            red[0][i >> 6] = emax;
-            red[1][i >> 6] = zmax;
+        if (lane == 0) {
+            red[0][w] = emax;
+            red[1][w] = zmax;
         }
         __syncthreads();
-        if (i == 0 && ok) {
-            const uint32_t e = red[0][0] > red[0][1] ? red[0][0] : red[0][1];
-            const uint32_t z = red[1][0] > red[1][1] ? red[1][0] : red[1][1];
+        if (tid == 0 && ok) {
+            uint32_t e = red[0][0], z = red[1][0];
+            for (int v = 1; v < 4; ++v) {
+                e = e > red[0][v] ? e : red[0][v];
+                z = z > red[1][v] ? z : red[1][v];
+            }
             chain_bits[id] = e;
             chain_bits[(size_t)B * ncs + id] = z;
         }
@@ -495,7 +574,7 @@ int launch_fixup_big(int mode, bool flip, int B, int T, int M, const float *J, c
     const int grid = B * ncs;
     KTimer kt(mode == 2 ? "k_fixup_dense_rev" : "k_fixup_dense_fwd", st);
 #define FXB(MO, F)                                                                                                  \
-    hipLaunchKernelGGL((k_fixup_big<MO, F>), dim3(grid), dim3(BG), 0, st, J, rhs, rhs_sign, carry_in, z, out, zsel, \
+    hipLaunchKernelGGL((k_fixup_big<MO, F>), dim3(grid), dim3(256), 0, st, J, rhs, rhs_sign, carry_in, z, out, zsel, \
                        chain_bits, active, B, T, M, C, ncs)
     if (mode == 0) FXB(0, false);
     else if (mode == 1) { if (flip) FXB(1, true); else FXB(1, false); }

@@ -774,52 +774,56 @@ __global__ __launch_bounds__(256) void k_resjac_shmfma(const ShArgs a, const flo
                 zt[j][q] = e ? v : 0.f;
                 zc[j][q] = e ? cur.zc[j][q] : 0.f;
             }
-        v4f F[NI];
-#pragma unroll
-        for (int I = 0; I < NI; ++I) F[I] = (v4f){0.f, 0.f, 0.f, 0.f};
-        for (int w = 0; w < LW; ++w) {
-            uint32_t word = 0u;
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int lt = 2 * w + h;
-                if (lt >= nlt) break;
-                const float4 hq = *reinterpret_cast<const float4 *>(h2s + 16 * lt + 4 * g);
-                v4f u = {hq.x, hq.y, hq.z, hq.w};
-#pragma unroll
-                for (int j = 0; j < NI; ++j) {
-                    const float4 aq = *reinterpret_cast<const float4 *>(w2s + (16 * lt + c) * MQ + 16 * j + 4 * g);
-                    u = mfma16x16x4(aq.x, zt[j][0], u);
-                    u = mfma16x16x4(aq.y, zt[j][1], u);
-                    u = mfma16x16x4(aq.z, zt[j][2], u);
-                    u = mfma16x16x4(aq.w, zt[j][3], u);
+        // a tile whose sequences have all stopped (a pass queued past their convergence) does no
+        // work (the branch is wave-uniform)
+        if (__builtin_amdgcn_ballot_w64(rok) != 0ull) {
+            v4f F[NI];
+    #pragma unroll
+            for (int I = 0; I < NI; ++I) F[I] = (v4f){0.f, 0.f, 0.f, 0.f};
+            for (int w = 0; w < LW; ++w) {
+                uint32_t word = 0u;
+    #pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int lt = 2 * w + h;
+                    if (lt >= nlt) break;
+                    const float4 hq = *reinterpret_cast<const float4 *>(h2s + 16 * lt + 4 * g);
+                    v4f u = {hq.x, hq.y, hq.z, hq.w};
+    #pragma unroll
+                    for (int j = 0; j < NI; ++j) {
+                        const float4 aq = *reinterpret_cast<const float4 *>(w2s + (16 * lt + c) * MQ + 16 * j + 4 * g);
+                        u = mfma16x16x4(aq.x, zt[j][0], u);
+                        u = mfma16x16x4(aq.y, zt[j][1], u);
+                        u = mfma16x16x4(aq.z, zt[j][2], u);
+                        u = mfma16x16x4(aq.w, zt[j][3], u);
+                    }
+    #pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const bool on = u[r] > 0.f;
+                        word |= (on ? 1u : 0u) << (16 * h + 4 * g + r);
+                        u[r] = on ? u[r] : 0.f;
+                    }
+    #pragma unroll
+                    for (int I = 0; I < NI; ++I) {
+                        const float4 aq = *reinterpret_cast<const float4 *>(w1s + (16 * I + c) * LQ + 16 * lt + 4 * g);
+                        F[I] = mfma16x16x4(aq.x, u[0], F[I]);
+                        F[I] = mfma16x16x4(aq.y, u[1], F[I]);
+                        F[I] = mfma16x16x4(aq.z, u[2], F[I]);
+                        F[I] = mfma16x16x4(aq.w, u[3], F[I]);
+                    }
                 }
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const bool on = u[r] > 0.f;
-                    word |= (on ? 1u : 0u) << (16 * h + 4 * g + r);
-                    u[r] = on ? u[r] : 0.f;
-                }
-#pragma unroll
-                for (int I = 0; I < NI; ++I) {
-                    const float4 aq = *reinterpret_cast<const float4 *>(w1s + (16 * I + c) * LQ + 16 * lt + 4 * g);
-                    F[I] = mfma16x16x4(aq.x, u[0], F[I]);
-                    F[I] = mfma16x16x4(aq.y, u[1], F[I]);
-                    F[I] = mfma16x16x4(aq.z, u[2], F[I]);
-                    F[I] = mfma16x16x4(aq.w, u[3], F[I]);
-                }
+                word |= (uint32_t)__shfl_xor((int)word, 16, 64);
+                word |= (uint32_t)__shfl_xor((int)word, 32, 64);
+                if (g == 0 && rok) masks[(size_t)rowc * LW + w] = word;
             }
-            word |= (uint32_t)__shfl_xor((int)word, 16, 64);
-            word |= (uint32_t)__shfl_xor((int)word, 32, 64);
-            if (g == 0 && rok) masks[(size_t)rowc * LW + w] = word;
-        }
-        if (rok) {
-#pragma unroll
-            for (int I = 0; I < NI; ++I)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int i = 16 * I + 4 * g + r;
-                    if (i < M) r_out[(size_t)rowc * M + i] = zc[I][r] - (fmaf(dA[I][r], zt[I][r], F[I][r]) + h1v[I][r]);
-                }
+            if (rok) {
+    #pragma unroll
+                for (int I = 0; I < NI; ++I)
+    #pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int i = 16 * I + 4 * g + r;
+                        if (i < M) r_out[(size_t)rowc * M + i] = zc[I][r] - (fmaf(dA[I][r], zt[I][r], F[I][r]) + h1v[I][r]);
+                    }
+            }
         }
         cur = nxt;
         r1 = r2;

@@ -112,6 +112,36 @@ def test_shallow_solve_and_adjoint(M, L, N, B, T, alpha, chunk):
         assert rel_inf(out["grads"][k].cpu().numpy(), gr[k]) < TOL, k
 
 
+@pytest.mark.parametrize("path", ["fused", "fixed-order residual", "stored Jacobian"])
+def test_shallow_nonfinite_and_not_converged(path):
+    """A NaN input ends its sequence as non-finite after the damped retries, and an update cap of
+    one leaves both sequences unconverged after one update: with the pass-end control in the
+    Jacobian-vector fix-up (the default), with the fixed-order residual (k_seq_ctl), and on the
+    stored-Jacobian path."""
+    env = {"fused": {}, "fixed-order residual": {"DEER_SH_RESMFMA": "0"},
+           "stored Jacobian": {"DEER_SH_FUSED": "0"}}[path]
+    c = _case(6, 20, 3, 2, 300, 0.2, 23)
+    m = oracle_model(c)
+    x = c.x.copy()
+    x[1, 70, 1] = np.nan
+    try:
+        os.environ.update(env)
+        say("shallow NaN input", path)
+        res = D.deer_solve(m, x, 0.2, 3, tol=1e-5, check=False)
+        assert res["status"] == 3                      # DEER_ERR_NONFINITE
+        say("shallow max_iter=1", path)
+        res = D.deer_solve(m, c.x, 0.2, 3, tol=1e-5, max_iter=1, check=False)
+        assert res["status"] == 2                      # DEER_ERR_NOT_CONVERGED
+        assert res["iters"] == [1, 1]
+        say("shallow to tolerance", path)
+        res = D.deer_solve(m, c.x, 0.2, 3, tol=1e-5, max_iter=100)
+        assert res["status"] == 0
+        assert rel_inf(res["z"].cpu().numpy(), O.rollout(m, c.x, 0.2, 3)) < TOL
+    finally:
+        for k in env:
+            os.environ.pop(k, None)
+
+
 @pytest.mark.parametrize("M,L,N,B,T,chunk,bound", [(16, 64, 16, 3, 300, 0, 0.05), (20, 40, 5, 3, 200, 32, 0.2)])
 def test_shallow_safeguard_rejections_reach_rollout(M, L, N, B, T, chunk, bound):
     """Rejected updates retried with the damped stored Jacobians gamma J~ still reach the

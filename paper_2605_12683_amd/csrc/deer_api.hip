@@ -227,10 +227,9 @@ static int choose_chunk(int B, int T, int MP, bool sh_fused = false) {
     // MP = 64 runs one chain per wave at two waves per SIMD: 8192 chains keep the tail of a
     // pass (fewer active sequences) spread over the machine
     if (MP == 128) {
-        // one 4-wave workgroup per chain; fewer than 96 chunks per sequence (one carry level)
-        long C = (total + 1023) / 1024;
-        const long minC = (T + 94) / 95;
-        if (C < minC) C = minC;
+        // one 4-wave workgroup per chain, one chain per CU (its staged tiles fill the LDS): about
+        // 256 chains, at least 16 steps per chunk
+        long C = (total + 255) / 256;
         if (C < 16) C = 16;
         if (C > T) C = T;
         return (int)C;

@@ -7,11 +7,11 @@
 //                         accumulators are the B operand, the step's Jacobian rows the A operand,
 //                         read as 16-byte vectors); the chunk-local solution u <- E_t u + rhs on
 //                         the vector units through LDS
-//   k_carry_big           one 128-thread block per sequence: carries across the chunks (fewer
-//                         than 96 per sequence at this width, so one level)
+//   k_carry_big           one 256-thread block per walk: carries across the chunks, one level,
+//                         or two with k_carry_group_big (group maps on the matrix cores)
 //   k_fixup_big           one 128-thread block per chain: each chunk re-run from its carry
-//   k_resjac_big          residual, masks (the fixed-order float32 decision) and F, one row at a
-//                         time per block, W1 and W2 in LDS
+//   k_resjac_big          residual, masks (the fixed-order float32 decision) and F, one row per
+//                         wave, W1 and W2 in LDS
 //   k_jacform_big         J~ = diag(A p) + W1 diag(m) (W2 P) on the matrix cores, 4 waves per
 //                         row, two column tiles each
 //   k_grads_big           per-block partial sums of the shallow gradients (layout of
@@ -159,28 +159,190 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
     if (tid < BG) vout[(size_t)id * BG + tid] = ub[cur][tid];
 }
 
-// carries across the chunks of each sequence, in processing order (REV: from the last chunk):
-// carry_in[c] = the state entering chunk c;  next = A_c carry + v_c with A_c = P_c (P_c^T in REV)
+// carries across the chunks of each sequence, in processing order k (REV: chunk c = ncs - 1 - k):
+// carry_in[c] = the state entering chunk c;  next = A_k carry + v_c with A_k = P_c (P_c^T in REV).
+// Long chunk sequences use two levels: groups of G consecutive k composed into one map (Q_j, u_j)
+// on the matrix cores (k_carry_group_big, all groups in parallel), a walk over the group maps, and
+// every group re-walked from its carry.  Serial depth G + ncs / G + G instead of ncs.
+constexpr int FST = BG + 1;   // LDS row stride of a tile read along rows and along columns
+
+// one walk of G consecutive k per 256-thread block (G = ncs: a whole sequence), from zero or from
+// the walk's start vector.  Lane l of wave w forms half hh = l / 32 of row i = 32 w + l % 32 of
+// A_k y; each step's P_c is staged in LDS with coalesced loads, the next one's in flight.
 template <bool REV>
-__global__ __launch_bounds__(BG) void k_carry_big(const float *__restrict__ P, const float *__restrict__ v,
-                                                  float *__restrict__ carry_in, const int *__restrict__ active,
-                                                  int ncs) {
-    __shared__ float cs[BG];
-    const int b = blockIdx.x, i = threadIdx.x;
+__global__ __launch_bounds__(256) void k_carry_big(const float *__restrict__ P, const float *__restrict__ v,
+                                                   float *__restrict__ carry_in, const int *__restrict__ active,
+                                                   int ncs, int G, const float *__restrict__ start) {
+    __shared__ float js[2][BG][FST];
+    __shared__ float ys[2][BG];
+    const int ngroups = (ncs + G - 1) / G;
+    const int b = blockIdx.x / ngroups, j = blockIdx.x % ngroups;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hh = lane >> 5, i = 32 * w + (lane & 31);
     if (active && !active[b]) return;
-    float cur = 0.f;
-    for (int step = 0; step < ncs; ++step) {
-        const int cc = REV ? ncs - 1 - step : step;
-        const size_t id = (size_t)b * ncs + cc;
-        carry_in[id * BG + i] = cur;
-        cs[i] = cur;
+    const int k0 = j * G, k1 = min(k0 + G, ncs);
+    auto chunk = [&](int k) { return (size_t)b * ncs + (REV ? ncs - 1 - k : k); };
+    // staging: thread tid takes the 16-byte groups tid + 256 q (q < 16) of the 128 x 128 map,
+    // row (tid + 256 q) / 32, columns 4 (tid % 32) .. + 3
+    float4 pre[16];
+    float vpre = 0.f;
+    auto stage_load = [&](int k) {
+        const size_t id = chunk(k);
+        const float4 *P4 = reinterpret_cast<const float4 *>(P + id * BG * BG);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) pre[q] = P4[tid + 256 * q];
+        vpre = v[id * BG + i];
+    };
+    auto stage_store = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int e4 = tid + 256 * q, row = e4 >> 5, c4 = (e4 & 31) * 4;
+            js[buf][row][c4] = pre[q].x;
+            js[buf][row][c4 + 1] = pre[q].y;
+            js[buf][row][c4 + 2] = pre[q].z;
+            js[buf][row][c4 + 3] = pre[q].w;
+        }
+    };
+    if (tid < BG) ys[0][tid] = start ? start[((size_t)b * ngroups + j) * BG + tid] : 0.f;
+    stage_load(k0);
+    stage_store(0);
+    float vc = vpre;
+    __syncthreads();
+    int cur = 0;
+    const int q0 = 64 * hh;
+    for (int k = k0; k < k1; ++k) {
+        const bool more = k + 1 < k1;
+        if (more) stage_load(k + 1);   // in flight during this step
+        if (hh == 0) carry_in[chunk(k) * BG + i] = ys[cur][i];
+        // half hh of the sum over q in [64 hh, 64 hh + 64), walked from 32 hh on: with the row
+        // stride of 129 the 64 lanes of a read fall on distinct banks, along rows and columns
+        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll 4
+        for (int u = 0; u < 64; u += 4) {
+            const int q = q0 + ((u + 32 * hh) & 63);
+            const float e0 = REV ? js[cur][q][i] : js[cur][i][q];
+            const float e1 = REV ? js[cur][q + 1][i] : js[cur][i][q + 1];
+            const float e2 = REV ? js[cur][q + 2][i] : js[cur][i][q + 2];
+            const float e3 = REV ? js[cur][q + 3][i] : js[cur][i][q + 3];
+            a0 = fmaf(e0, ys[cur][q], a0);
+            a1 = fmaf(e1, ys[cur][q + 1], a1);
+            a2 = fmaf(e2, ys[cur][q + 2], a2);
+            a3 = fmaf(e3, ys[cur][q + 3], a3);
+        }
+        float part = (a0 + a1) + (a2 + a3);
+        part += __shfl_xor(part, 32, 64);
+        if (hh == 0) ys[cur ^ 1][i] = part + vc;
+        if (more) {
+            stage_store(cur ^ 1);   // that buffer's reads ended at the previous barrier
+            vc = vpre;
+        }
         __syncthreads();
-        const float *Pc = P + id * BG * BG;
-        float a = v[id * BG + i];
-        for (int k = 0; k < BG; ++k) a = fmaf(REV ? Pc[(size_t)k * BG + i] : Pc[(size_t)i * BG + k], cs[k], a);
-        __syncthreads();
-        cur = a;
+        cur ^= 1;
     }
+}
+
+// group maps in processing order: Q_j = A_{k1-1} ... A_{k0} and u_j = the group's walk from zero.
+// Q accumulates on the matrix cores as the chunk product above does (A_k staged in LDS, transposed
+// there in REV, the next one's loads in flight; Q in the k-permuted accumulator layout that is the
+// next step's B operand); u by thread pairs over the staged rows.
+template <bool REV>
+__global__ __launch_bounds__(256) void k_carry_group_big(const float *__restrict__ P, const float *__restrict__ v,
+                                                         float *__restrict__ gq, float *__restrict__ gu,
+                                                         const int *__restrict__ active, int ncs, int G) {
+    __shared__ __align__(16) float js[2][BG][JST];
+    __shared__ __align__(16) float ub[2][BG];
+    const int ngroups = (ncs + G - 1) / G;
+    const int b = blockIdx.x / ngroups, j = blockIdx.x % ngroups;
+    const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
+    if (active && !active[b]) return;
+    const int k0 = j * G, k1 = min(k0 + G, ncs);
+    auto chunk = [&](int k) { return (size_t)b * ncs + (REV ? ncs - 1 - k : k); };
+    const int ui = tid >> 1, hh = tid & 1;
+    float4 pre[16];
+    float vpre = 0.f;
+    auto stage_load = [&](int k) {
+        const size_t id = chunk(k);
+        const float4 *P4 = reinterpret_cast<const float4 *>(P + id * BG * BG);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) pre[q] = P4[tid + 256 * q];
+        if (hh == 0) vpre = v[id * BG + ui];
+    };
+    auto stage_store = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int e4 = tid + 256 * q, row = e4 >> 5, c4 = (e4 & 31) * 4;
+            if (REV) {
+                js[buf][c4][row] = pre[q].x;
+                js[buf][c4 + 1][row] = pre[q].y;
+                js[buf][c4 + 2][row] = pre[q].z;
+                js[buf][c4 + 3][row] = pre[q].w;
+            } else {
+                *reinterpret_cast<float4 *>(&js[buf][row][c4]) = pre[q];
+            }
+        }
+    };
+    // accumulators: acc[I][Jt][r] = Q[16 I + 4 g + r][32 wv + 16 Jt + c]
+    v4f acc[8][2];
+#pragma unroll
+    for (int I = 0; I < 8; ++I)
+#pragma unroll
+        for (int Jt = 0; Jt < 2; ++Jt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[I][Jt][r] = (16 * I + 4 * g + r == 32 * wv + 16 * Jt + c) ? 1.f : 0.f;
+    if (tid < BG) ub[0][tid] = 0.f;
+    stage_load(k0);
+    stage_store(0);
+    float vc = vpre;
+    __syncthreads();
+    int cur = 0;
+    for (int k = k0; k < k1; ++k) {
+        const bool more = k + 1 < k1;
+        if (more) stage_load(k + 1);   // in flight during this step
+        v4f old[8][2];
+#pragma unroll
+        for (int I = 0; I < 8; ++I)
+#pragma unroll
+            for (int Jt = 0; Jt < 2; ++Jt) {
+                old[I][Jt] = acc[I][Jt];
+                acc[I][Jt] = (v4f){0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+        for (int I = 0; I < 8; ++I) {
+            float4 a[8];
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj) a[jj] = *reinterpret_cast<const float4 *>(&js[cur][16 * I + c][16 * jj + 4 * g]);
+#pragma unroll
+            for (int Jt = 0; Jt < 2; ++Jt) {
+                v4f s = acc[I][Jt];
+#pragma unroll
+                for (int jj = 0; jj < 8; ++jj) {
+                    s = mfma16x16x4(a[jj].x, old[jj][Jt][0], s);
+                    s = mfma16x16x4(a[jj].y, old[jj][Jt][1], s);
+                    s = mfma16x16x4(a[jj].z, old[jj][Jt][2], s);
+                    s = mfma16x16x4(a[jj].w, old[jj][Jt][3], s);
+                }
+                acc[I][Jt] = s;
+            }
+        }
+        // u <- A_k u + v_c: thread pair (row ui, half hh) sums every other entry of the row
+        float part = 0.f;
+        for (int q = hh; q < BG; q += 2) part = fmaf(js[cur][ui][q], ub[cur][q], part);
+        part += __shfl_xor(part, 1, 64);
+        if (hh == 0) ub[cur ^ 1][ui] = part + vc;
+        if (more) {
+            stage_store(cur ^ 1);   // that buffer's reads ended at the previous barrier
+            vc = vpre;
+        }
+        __syncthreads();
+        cur ^= 1;
+    }
+    float *q = gq + ((size_t)b * ngroups + j) * BG * BG;
+#pragma unroll
+    for (int I = 0; I < 8; ++I)
+#pragma unroll
+        for (int Jt = 0; Jt < 2; ++Jt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) q[(16 * I + 4 * g + r) * BG + 32 * wv + 16 * Jt + c] = acc[I][Jt][r];
+    if (tid < BG) gu[((size_t)b * ngroups + j) * BG + tid] = ub[cur][tid];
 }
 
 // MODE 0: Newton fix-up (next iterate = current + Delta, per-chain max |Delta| and max |z|);
@@ -190,7 +352,6 @@ __global__ __launch_bounds__(BG) void k_carry_big(const float *__restrict__ P, c
 // loads, the next step's loads (and its right-hand side and iterate) in flight during this step.
 // With a row stride of 129 floats and the second half's walk started 32 entries in, the 64 lanes
 // of a read fall on distinct banks, for rows (MODE 0, 1) and for columns (MODE 2).
-constexpr int FST = BG + 1;
 
 template <int MODE, bool FLIP>
 __global__ __launch_bounds__(256) void k_fixup_big(const float *__restrict__ J, const float *__restrict__ rhs,
@@ -342,59 +503,68 @@ __device__ __forceinline__ float big_forced(const ShArgs &a, const float *z, int
     return __fadd_rn(__fmul_rn(p, zp), __fmul_rn(a.alpha, xs));
 }
 
-// LDS: W1 [M][L] | W2 [L][M] | z~ [BG] | relu(u) [L]
+// One row per wave, the four waves of a block on their own rows; LDS: W2^T [M][L] | W1^T [L][M],
+// so that the lanes of a read take consecutive words.  Lane l < L forms the hidden pre-activation
+// u_l left to right from h2 (a rounding after every multiply and add: the fixed-order float32
+// decision), with z~_j broadcast from lane j % 64 of the wave's registers; lanes i and i + 64 form
+// F_i and r_i from relu(u), broadcast the same way.
 __global__ __launch_bounds__(256) void k_resjac_big(const ShArgs a, const float *zbuf, const float *zalt,
                                                     const int *__restrict__ zsel, float *__restrict__ F_out,
                                                     float *__restrict__ r_out, uint32_t *__restrict__ masks,
                                                     const int *__restrict__ active) {
     extern __shared__ __align__(16) float smem[];
-    const int M = a.M, L = a.L, T = a.T, tid = threadIdx.x;
-    float *w1 = smem, *w2 = w1 + (size_t)M * L, *zt = w2 + (size_t)L * M, *ru = zt + BG;
+    const int M = a.M, L = a.L, T = a.T, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    float *w2t = smem, *w1t = w2t + (size_t)M * L;
     for (int e = tid; e < M * L; e += 256) {
-        w1[e] = a.W1[e];
-        w2[e] = a.W2[e];
+        const int i = e / L, l = e % L;   // W1[i][l]; W2[l][i] at the same (i, l)
+        w1t[(size_t)l * M + i] = a.W1[e];
+        w2t[(size_t)i * L + l] = a.W2[(size_t)l * M + i];
     }
     const int LW = (L + 31) / 32;
     const long rows = (long)a.B * T;
     __syncthreads();
-    for (long row = blockIdx.x; row < rows; row += gridDim.x) {
+    for (long row = (long)blockIdx.x * 4 + wv; row < rows; row += (long)gridDim.x * 4) {
         const int b = (int)(row / T), s = (int)(row % T);
-        const bool on = !active || active[b];   // block-uniform
-        if (!on) continue;
+        if (active && !active[b]) continue;   // wave-uniform
         const float *z = cur_iter(zbuf, zalt, zsel, b);
-        if (tid < M) zt[tid] = big_forced(a, z, b, s, tid);
-        __syncthreads();
-        // hidden pre-activations left to right from h2, a rounding after every multiply and add
-        for (int l = tid; l < L; l += 256) {
-            float u = a.h2 ? a.h2[l] : 0.f;
-            for (int j = 0; j < M; ++j) u = __fadd_rn(u, __fmul_rn(w2[(size_t)l * M + j], zt[j]));
-            ru[l] = u > 0.f ? u : 0.f;
+        const int i1 = lane + 64;
+        const float zt0 = lane < M ? big_forced(a, z, b, s, lane) : 0.f;
+        const float zt1 = i1 < M ? big_forced(a, z, b, s, i1) : 0.f;
+        float u = 0.f;
+        if (lane < L) {
+            u = a.h2 ? a.h2[lane] : 0.f;
+            const float *wr = w2t + lane;
+            const int m0 = M < 64 ? M : 64;
+            for (int j = 0; j < m0; ++j)
+                u = __fadd_rn(u, __fmul_rn(wr[(size_t)j * L], __int_as_float(__builtin_amdgcn_readlane(__float_as_int(zt0), j))));
+            for (int j = 64; j < M; ++j)
+                u = __fadd_rn(u, __fmul_rn(wr[(size_t)j * L], __int_as_float(__builtin_amdgcn_readlane(__float_as_int(zt1), j - 64))));
         }
-        __syncthreads();
-        if (masks) {
-            for (int w = tid; w < LW; w += 256) {
-                uint32_t bits = 0u;
-                for (int k = 0; k < 32; ++k) {
-                    const int l = 32 * w + k;
-                    if (l < L && ru[l] > 0.f) bits |= 1u << k;
-                }
-                masks[(size_t)row * LW + w] = bits;
-            }
+        const float ru = (lane < L && u > 0.f) ? u : 0.f;
+        const uint64_t on = __builtin_amdgcn_ballot_w64(lane < L && u > 0.f);
+        if (masks && lane < LW) masks[(size_t)row * LW + lane] = (uint32_t)(on >> (32 * lane));
+        float f0 = 0.f, f1 = 0.f;
+        for (int l = 0; l < L; ++l) {
+            const float rl = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ru), l));
+            f0 = fmaf(w1t[(size_t)l * M + lane], rl, f0);
+            if (i1 < M) f1 = fmaf(w1t[(size_t)l * M + i1], rl, f1);
         }
-        if (tid < M) {
-            float f = 0.f;
-            for (int l = 0; l < L; ++l) f = fmaf(w1[(size_t)tid * L + l], ru[l], f);
-            f = fmaf(a.A[tid], zt[tid], f) + (a.h1 ? a.h1[tid] : 0.f);
-            const size_t e = (size_t)row * M + tid;
-            if (F_out) F_out[e] = f;
-            if (r_out) r_out[e] = z[e] - f;
+        const size_t e0 = (size_t)row * M;
+        if (lane < M) {
+            const float f = fmaf(a.A[lane], zt0, f0) + (a.h1 ? a.h1[lane] : 0.f);
+            if (F_out) F_out[e0 + lane] = f;
+            if (r_out) r_out[e0 + lane] = z[e0 + lane] - f;
         }
-        __syncthreads();
+        if (i1 < M) {
+            const float f = fmaf(a.A[i1], zt1, f1) + (a.h1 ? a.h1[i1] : 0.f);
+            if (F_out) F_out[e0 + i1] = f;
+            if (r_out) r_out[e0 + i1] = z[e0 + i1] - f;
+        }
     }
 }
 
-// J~_s = Cd (or diag(A p)) + W1 diag(m_s) V with V = W2 diag(p) (or the given W2 P): one row per
-// block, wave wv computes the column tiles 2 wv, 2 wv + 1 of all 8 row tiles.  LDS: W1 [BG][LP],
+// J~_s = Cd (or diag(A p)) + W1 diag(m_s) V with V = W2 diag(p) (or the given W2 P): one row at a
+// time per block, the blocks walking the rows, wave wv computes the column tiles 2 wv, 2 wv + 1 of all 8 row tiles.  LDS: W1 [BG][LP],
 // V^T [BG][LP], zero padded (LP = L rounded up to 16).
 __global__ __launch_bounds__(256) void k_jacform_big(const ShArgs a, const uint32_t *__restrict__ masks,
                                                      float *__restrict__ Jout, const int *__restrict__ active,
@@ -413,12 +583,28 @@ __global__ __launch_bounds__(256) void k_jacform_big(const ShArgs a, const uint3
     __syncthreads();
     const int wv = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
     const int LW = (L + 31) / 32;
+    const auto cd_rs = bounded_rsrc(a.Cd, a.Cd ? (uint32_t)M * M * 4u : 0u);
     const int t_lo = a.t_hi > a.t_lo ? a.t_lo : 0;
     const int len = a.t_hi > a.t_lo ? a.t_hi - a.t_lo : T;
     const long rows = (long)a.B * len;
+    auto grow_of = [&](long r) {
+        const long bb = r / len;
+        return bb * T + t_lo + (r - bb * len);
+    };
+    // the next row's mask words (L <= 64: at most two) are loaded while this row is formed
+    uint32_t wn0 = 0u, wn1 = 0u;
+    auto fetch = [&](long r) {
+        if (r >= rows) return;
+        const uint32_t *mw = masks + (size_t)grow_of(r) * LW;
+        wn0 = mw[0];
+        wn1 = LW > 1 ? mw[1] : 0u;
+    };
+    fetch(blockIdx.x);
     for (long r0 = blockIdx.x; r0 < rows; r0 += gridDim.x) {
         const long bb = r0 / len;
-        const long grow = bb * T + t_lo + (r0 - bb * len);
+        const long grow = grow_of(r0);
+        const uint32_t wc0 = wn0, wc1 = wn1;
+        fetch(r0 + gridDim.x);
         if (active && !active[bb]) continue;
         v4f acc[8][2];
 #pragma unroll
@@ -426,8 +612,8 @@ __global__ __launch_bounds__(256) void k_jacform_big(const ShArgs a, const uint3
 #pragma unroll
             for (int Jt = 0; Jt < 2; ++Jt) acc[I][Jt] = (v4f){0.f, 0.f, 0.f, 0.f};
         for (int j = 0; j < LP / 16; ++j) {
-            const int word = (16 * j) >> 5, sh = 16 * (j & 1) + 4 * g;
-            const uint32_t w = masks[(size_t)grow * LW + word];
+            const int sh = 16 * (j & 1) + 4 * g;
+            const uint32_t w = j < 2 ? wc0 : wc1;
             float4 bv[2];
 #pragma unroll
             for (int Jt = 0; Jt < 2; ++Jt) {
@@ -449,21 +635,27 @@ __global__ __launch_bounds__(256) void k_jacform_big(const ShArgs a, const uint3
                 }
             }
         }
-        float *Jp = Jout + (size_t)grow * M * M;
+        // stores through a resource bounded at J~_s's end: rows past M fall outside it, columns
+        // past M take an offset outside it
+        const auto rs = bounded_rsrc(Jout + (size_t)grow * M * M, (uint32_t)M * M * 4u);
         const float gm = gamma ? gamma[bb] : 1.f;
 #pragma unroll
-        for (int I = 0; I < 8; ++I)
+        for (int Jt = 0; Jt < 2; ++Jt) {
+            const int col = 32 * wv + 16 * Jt + c;
+            const uint32_t vo = col < M ? 4u * (uint32_t)(4 * g * M + col) : kOffLane;
+            // the diagonal entry (col, col) sits in row tile col / 16 at 4 g + r = col % 16
+            const float dg = (!a.Cd && col < M) ? a.A[col] * (col < N ? p1 : 1.f) : 0.f;
 #pragma unroll
-            for (int Jt = 0; Jt < 2; ++Jt)
+            for (int I = 0; I < 8; ++I)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int row = 16 * I + 4 * g + r, col = 32 * wv + 16 * Jt + c;
-                    if (row < M && col < M) {
-                        const float d = a.Cd ? a.Cd[row * M + col]
-                                             : (row == col ? a.A[row] * (row < N ? p1 : 1.f) : 0.f);
-                        Jp[row * M + col] = gm * (acc[I][Jt][r] + d);
-                    }
+                    // lane offset of row 16 I + 4 g + r (kOffLane plus a row offset stays outside)
+                    const uint32_t vr = vo + 4u * (uint32_t)M * (uint32_t)(16 * I + r);
+                    float d = (16 * I + 4 * g + r == col) ? dg : 0.f;
+                    if (a.Cd) d = bload(cd_rs, vr, 0);
+                    bstore_u(rs, __float_as_uint(gm * (acc[I][Jt][r] + d)), vr, 0);
                 }
+        }
     }
 }
 
@@ -560,10 +752,27 @@ int launch_chunk_product_big(bool rev, bool flip, int B, int T, int M, const flo
 }
 
 int launch_carry_big(bool rev, const float *P, const float *v, float *carry_in, const int *active, int B, int ncs,
-                     hipStream_t st) {
+                     int G, float *gws, hipStream_t st) {
     KTimer kt("k_carry", st);
-    if (rev) hipLaunchKernelGGL(k_carry_big<true>, dim3(B), dim3(BG), 0, st, P, v, carry_in, active, ncs);
-    else hipLaunchKernelGGL(k_carry_big<false>, dim3(B), dim3(BG), 0, st, P, v, carry_in, active, ncs);
+    if (!G) {
+        if (rev) hipLaunchKernelGGL(k_carry_big<true>, dim3(B), dim3(256), 0, st, P, v, carry_in, active, ncs, ncs, nullptr);
+        else hipLaunchKernelGGL(k_carry_big<false>, dim3(B), dim3(256), 0, st, P, v, carry_in, active, ncs, ncs, nullptr);
+        DEER_LAUNCH_CHECK("k_carry_big");
+        return DEER_OK;
+    }
+    // workspace: group maps [B][ng][BG][BG], their walks from zero [B][ng][BG], group carries
+    const int ng = (ncs + G - 1) / G;
+    float *gq = gws;
+    float *gu = gq + (size_t)B * ng * BG * BG;
+    float *gc = gu + (size_t)B * ng * BG;
+    const int grid = B * ng;
+    if (rev) hipLaunchKernelGGL(k_carry_group_big<true>, dim3(grid), dim3(256), 0, st, P, v, gq, gu, active, ncs, G);
+    else hipLaunchKernelGGL(k_carry_group_big<false>, dim3(grid), dim3(256), 0, st, P, v, gq, gu, active, ncs, G);
+    DEER_LAUNCH_CHECK("k_carry_group_big");
+    hipLaunchKernelGGL(k_carry_big<false>, dim3(B), dim3(256), 0, st, gq, gu, gc, active, ng, ng, nullptr);
+    DEER_LAUNCH_CHECK("k_carry_big");
+    if (rev) hipLaunchKernelGGL(k_carry_big<true>, dim3(grid), dim3(256), 0, st, P, v, carry_in, active, ncs, G, gc);
+    else hipLaunchKernelGGL(k_carry_big<false>, dim3(grid), dim3(256), 0, st, P, v, carry_in, active, ncs, G, gc);
     DEER_LAUNCH_CHECK("k_carry_big");
     return DEER_OK;
 }
@@ -584,14 +793,17 @@ int launch_fixup_big(int mode, bool flip, int B, int T, int M, const float *J, c
     return DEER_OK;
 }
 
-size_t big_resjac_lds(int M, int L) { return ((size_t)2 * M * L + BG + L) * sizeof(float); }
+size_t big_resjac_lds(int M, int L) { return (size_t)2 * M * L * sizeof(float); }
 size_t big_jacform_lds(int L) { return (size_t)2 * BG * ((L + 15) / 16 * 16) * sizeof(float); }
 size_t big_grads_lds(int M, int L) { return ((size_t)2 * M * L + 2 * BG + 2 * L) * sizeof(float); }
 
 int launch_resjac_big(const ShArgs &a, const float *z, const float *zalt, const int *zsel, float *F, float *r,
                       uint32_t *masks, const int *active, hipStream_t st) {
-    const long rows = (long)a.B * a.T;
-    const int grid = (int)(rows < 8192 ? rows : 8192);
+    // four rows per block; as many blocks as the LDS of the 256 CUs holds (160 KiB each, at most 8)
+    const long rows = (long)a.B * a.T, want = (rows + 3) / 4;
+    long per_cu = (long)(160 * 1024) / (long)big_resjac_lds(a.M, a.L);
+    per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
+    const int grid = (int)(want < 256 * per_cu ? want : 256 * per_cu);
     KTimer kt("k_resjac_shplrnn", st);
     hipLaunchKernelGGL(k_resjac_big, dim3(grid), dim3(256), big_resjac_lds(a.M, a.L), st, a, z, zalt, zsel, F, r,
                        masks, active);
@@ -601,8 +813,12 @@ int launch_resjac_big(const ShArgs &a, const float *z, const float *zalt, const 
 
 int launch_jacform_big(const ShArgs &a, const uint32_t *masks, float *J, const int *active, const float *gamma,
                        hipStream_t st) {
+    // every block walks rows with W1 and V staged once: as many blocks as the LDS holds (two per CU
+    // at L > 48)
     const long rows = (long)a.B * (a.t_hi > a.t_lo ? a.t_hi - a.t_lo : a.T);
-    const int grid = (int)(rows < 8192 ? rows : 8192);
+    long per_cu = (long)(160 * 1024) / (long)big_jacform_lds(a.L);
+    per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
+    const int grid = (int)(rows < 256 * per_cu ? rows : 256 * per_cu);
     const int LP = (a.L + 15) / 16 * 16;
     KTimer kt("k_jacform_shplrnn", st);
     hipLaunchKernelGGL(k_jacform_big, dim3(grid), dim3(256), big_jacform_lds(a.L), st, a, masks, J, active, gamma, LP);

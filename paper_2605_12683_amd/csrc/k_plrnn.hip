@@ -3594,6 +3594,13 @@ int launch_newton_pass16(const PlrnnArgs &a, float *z, float *zalt, const float 
 
 // two-level carry for chunk sequences at least this long
 static int carry_group_size(int MP, int ncs) {
+    if (MP == 128) {
+        // a group step (a 128 x 128 x 128 product on one CU) costs about six walk steps
+        if (ncs < 48) return 0;
+        int G = 4;
+        while (8 * G * G < ncs) G <<= 1;
+        return G;
+    }
     if (ncs < 96) return 0;
     int G = 8;
     while (2 * G * G < ncs) G <<= 1;   // a group step costs about twice a walk step
@@ -3610,8 +3617,8 @@ size_t carry_ws_floats(int MP, int B, int ncs) {
 int launch_carry(int MP, bool rev, const float *P, const float *v, float *carry_in, const int *active,
                  uint32_t *norm_bits, int B, int ncs, float *gws, hipStream_t st) {
     if (MP == 128) {
-        if (norm_bits || carry_group_size(MP, ncs)) return invalid_arg("width-128 carries take one level, no norms");
-        return launch_carry_big(rev, P, v, carry_in, active, B, ncs, st);
+        if (norm_bits) return invalid_arg("width-128 carries take no norms");
+        return launch_carry_big(rev, P, v, carry_in, active, B, ncs, gws ? carry_group_size(MP, ncs) : 0, gws, st);
     }
     KTimer kt("k_carry", st);
     const int G = gws ? carry_group_size(MP, ncs) : 0;

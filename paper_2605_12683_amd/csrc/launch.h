@@ -186,7 +186,7 @@ int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const floa
 int launch_chunk_product_big(bool rev, bool flip, int B, int T, int M, const float *J, const float *rhs,
                              float rhs_sign, float *P, float *v, const int *active, int C, int ncs, hipStream_t st);
 int launch_carry_big(bool rev, const float *P, const float *v, float *carry_in, const int *active, int B, int ncs,
-                     hipStream_t st);
+                     int G, float *gws, hipStream_t st);
 int launch_fixup_big(int mode, bool flip, int B, int T, int M, const float *J, const float *rhs, float rhs_sign,
                      const float *carry_in, float *z, float *out, const int *zsel, uint32_t *chain_bits,
                      const int *active, int C, int ncs, hipStream_t st);

@@ -50,7 +50,11 @@ def test_big_jacobian_masks_bitexact(M, L, N, T):
     assert rel_inf(out["J"].cpu().numpy().reshape(-1, M, M), ref["J"]) < 1e-5
 
 
-@pytest.mark.parametrize("B,T,M,chunk", [(2, 300, 65, 0), (1, 1000, 128, 0), (2, 513, 128, 37), (1, 1, 100, 0)])
+# (1, 1000, 128): 63 chunks, carries in two levels (groups of 4, the last of 3); (1, 3000, 128):
+# 188 chunks in groups of 8; (2, 1500, 97): two sequences of 94 chunks; (1, 900, 128) with 7-step
+# chunks: 129 chunks, the last group one chunk
+@pytest.mark.parametrize("B,T,M,chunk", [(2, 300, 65, 0), (1, 1000, 128, 0), (2, 513, 128, 37), (1, 1, 100, 0),
+                                         (1, 3000, 128, 0), (2, 1500, 97, 0), (1, 900, 128, 7)])
 @pytest.mark.parametrize("rev,tr", [(False, False), (True, True), (False, True), (True, False)])
 def test_big_dense_scan(B, T, M, chunk, rev, tr):
     if chunk:

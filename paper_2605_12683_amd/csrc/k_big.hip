@@ -32,7 +32,8 @@ __device__ __forceinline__ float eload(const float *__restrict__ Jp, int M, int 
 }
 
 // REV: the product covers steps [s0 + 1, min(s1 + 1, T)) (the reverse chunk map is its
-// transpose) and the local solution runs u_k = E_{k+1}^T u_{k+1} + rhs_k from k = s1 - 1 down.
+// transpose) and the local solution of u_k = E_{k+1}^T u_{k+1} + rhs_k (zero past the chunk) is
+// taken as the sum u_{s0} = sum_k (E_k ... E_{s0+1})^T rhs_k along the same sweep.
 // The step's E (128 x 128, zero outside M x M) is staged in LDS by the whole workgroup, the next
 // step's loads in flight while the matrix cores work on this one (double buffer), and every wave
 // reads its A operands there; the forward local solution reads the same tile.
@@ -53,12 +54,17 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
     const int lo = REV ? s0 + 1 : s0, hi = REV ? min(s1 + 1, T) : s1;
     const int plen = ok ? max(hi - lo, 0) : 0;
     const int ulen = ok ? s1 - s0 : 0;
-    const int nsteps = max(plen, ulen);
+    // REV: the chunk's local adjoint is u_{s0} = sum_k Q_k^T rhs_k with Q_k = E_k ... E_{s0+1}
+    // (Q_{s0} = I), and Q_k is the accumulated product after the step that takes E_k: the sweep
+    // that forms the product forms u_{s0} too, with the staged right-hand side of that step
+    const int nsteps = REV ? plen : max(plen, ulen);
     // staging: thread tid takes the 16-byte groups tid + 256 k (k < 16) of the 128 x 128 tile,
     // row (tid + 256 k) / 32, columns 4 ((tid + 256 k) % 32) .. + 3
     float4 pre[16];
+    float rpre = 0.f;
     auto stage_load = [&](int t) {
         const float *Jp = J + ((size_t)b * T + lo + t) * M * M;
+        if (REV) rpre = (tid < M && lo + t < s1) ? rhs[((size_t)b * T + lo + t) * M + tid] : 0.f;
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
             const int e4 = tid + 256 * k, row = e4 >> 5, c4 = (e4 & 31) * 4;
@@ -76,6 +82,7 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
             const int e4 = tid + 256 * k;
             *reinterpret_cast<float4 *>(&js[buf][e4 >> 5][(e4 & 31) * 4]) = pre[k];
         }
+        if (REV && tid < BG) ub[buf][tid] = rpre;
     };
     // accumulators: acc[I][Jt][r] = P[16 I + 4 g + r][32 wv + 16 Jt + c]
     v4f acc[8][2];
@@ -88,6 +95,7 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
     // local solution: thread pair (row i = tid / 2, half hh) sums half of the row
     const int ui = tid >> 1, hh = tid & 1;
     if (tid < BG) ub[0][tid] = 0.f;
+    float vsum[2] = {0.f, 0.f};   // REV: sum over the steps of (Q_k^T rhs_k)[32 wv + 16 Jt + c]
     if (plen > 0) {
         stage_load(0);
         stage_store(0);
@@ -124,22 +132,31 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
                     acc[I][Jt] = s;
                 }
             }
-        }
-        if (t < ulen) {
-            // forward: u_s = E_s u_{s-1} + sign rhs_s, s = s0 + t (E_s is the staged tile);
-            // reverse: k = s1 - 1 - t, u_k = E_{k+1}^T u_{k+1} + sign rhs_k (E_T does not exist:
-            // the first reverse step starts from zero)
-            const int k = REV ? s1 - 1 - t : s0 + t;
-            const int kj = REV ? k + 1 : k;
-            float part = 0.f;
-            if (ui < M && (!REV || kj < T)) {
-                if (REV) {
-                    const float *Jp = J + ((size_t)b * T + kj) * M * M;
-                    for (int q = hh; q < M; q += 2) part = fmaf(eload<FLIP>(Jp, M, q, ui), ub[cur][q], part);
-                } else {
-                    for (int q = hh; q < M; q += 2) part = fmaf(js[cur][ui][q], ub[cur][q], part);
+            if (REV && lo + t < s1) {
+                // rows 16 I + 4 g + r of column 32 wv + 16 Jt + c, then the four row groups g
+#pragma unroll
+                for (int Jt = 0; Jt < 2; ++Jt) {
+                    float part = 0.f;
+#pragma unroll
+                    for (int I = 0; I < 8; ++I) {
+                        const float4 rv = *reinterpret_cast<const float4 *>(&ub[cur][16 * I + 4 * g]);
+                        part = fmaf(acc[I][Jt][0], rv.x, part);
+                        part = fmaf(acc[I][Jt][1], rv.y, part);
+                        part = fmaf(acc[I][Jt][2], rv.z, part);
+                        part = fmaf(acc[I][Jt][3], rv.w, part);
+                    }
+                    part += __shfl_xor(part, 16, 64);
+                    part += __shfl_xor(part, 32, 64);
+                    vsum[Jt] += part;
                 }
             }
+        }
+        if (!REV && t < ulen) {
+            // u_s = E_s u_{s-1} + sign rhs_s, s = s0 + t (E_s is the staged tile)
+            const int k = s0 + t;
+            float part = 0.f;
+            if (ui < M)
+                for (int q = hh; q < M; q += 2) part = fmaf(js[cur][ui][q], ub[cur][q], part);
             part += __shfl_xor(part, 1, 64);
             if (hh == 0 && ui < BG)
                 ub[cur ^ 1][ui] = ui < M ? fmaf(rhs_sign, rhs[((size_t)b * T + k) * M + ui], part) : 0.f;
@@ -156,7 +173,18 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
         for (int Jt = 0; Jt < 2; ++Jt)
 #pragma unroll
             for (int r = 0; r < 4; ++r) P[(16 * I + 4 * g + r) * BG + 32 * wv + 16 * Jt + c] = acc[I][Jt][r];
-    if (tid < BG) vout[(size_t)id * BG + tid] = ub[cur][tid];
+    if (REV) {
+        if (g == 0) {
+#pragma unroll
+            for (int Jt = 0; Jt < 2; ++Jt) {
+                const int col = 32 * wv + 16 * Jt + c;
+                const float r0 = (col < M && s0 < s1) ? rhs[((size_t)b * T + s0) * M + col] : 0.f;
+                vout[(size_t)id * BG + col] = col < M ? rhs_sign * (r0 + vsum[Jt]) : 0.f;
+            }
+        }
+    } else if (tid < BG) {
+        vout[(size_t)id * BG + tid] = ub[cur][tid];
+    }
 }
 
 // carries across the chunks of each sequence, in processing order k (REV: chunk c = ncs - 1 - k):

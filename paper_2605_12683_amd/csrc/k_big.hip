@@ -62,18 +62,25 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
     // row (tid + 256 k) / 32, columns 4 ((tid + 256 k) % 32) .. + 3
     float4 pre[16];
     float rpre = 0.f;
+    // row-major E with M % 4 == 0: 16-byte loads through a resource bounded at the matrix's end
+    // (rows past M read zero) with one lane offset (columns past M: an offset outside it)
+    const bool fast = !FLIP && (M & 3) == 0;
+    const uint32_t vlane = ((tid & 31) * 4 + 3 < M) ? 4u * ((uint32_t)(tid >> 5) * M + (tid & 31) * 4) : kOffLane;
     auto stage_load = [&](int t) {
         const float *Jp = J + ((size_t)b * T + lo + t) * M * M;
         if (REV) rpre = (tid < M && lo + t < s1) ? rhs[((size_t)b * T + lo + t) * M + tid] : 0.f;
+        if (fast) {
+            const auto rs = bounded_rsrc(Jp, (uint32_t)M * M * 4u);
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+                pre[k] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)vlane, k * 32 * M, 0));
+            return;
+        }
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
             const int e4 = tid + 256 * k, row = e4 >> 5, c4 = (e4 & 31) * 4;
-            if (!FLIP && (M & 3) == 0 && row < M && c4 + 3 < M) {
-                pre[k] = *reinterpret_cast<const float4 *>(Jp + (size_t)row * M + c4);
-            } else {
-                pre[k] = make_float4(eload<FLIP>(Jp, M, row, c4), eload<FLIP>(Jp, M, row, c4 + 1),
-                                     eload<FLIP>(Jp, M, row, c4 + 2), eload<FLIP>(Jp, M, row, c4 + 3));
-            }
+            pre[k] = make_float4(eload<FLIP>(Jp, M, row, c4), eload<FLIP>(Jp, M, row, c4 + 1),
+                                 eload<FLIP>(Jp, M, row, c4 + 2), eload<FLIP>(Jp, M, row, c4 + 3));
         }
     };
     auto stage_store = [&](int buf) {
@@ -152,11 +159,22 @@ __global__ __launch_bounds__(256) void k_chunk_product_big(const float *__restri
             }
         }
         if (!REV && t < ulen) {
-            // u_s = E_s u_{s-1} + sign rhs_s, s = s0 + t (E_s is the staged tile)
+            // u_s = E_s u_{s-1} + sign rhs_s, s = s0 + t (E_s is the staged tile, zero outside M x M
+            // as u is): half hh of row ui, q in [64 hh, 64 hh + 64) four at a time, walked from 32
+            // entries in for hh = 1 so that the two halves of a lane pair fall on other banks
             const int k = s0 + t;
-            float part = 0.f;
-            if (ui < M)
-                for (int q = hh; q < M; q += 2) part = fmaf(js[cur][ui][q], ub[cur][q], part);
+            float p0 = 0.f, p1 = 0.f;
+#pragma unroll 4
+            for (int u = 0; u < 64; u += 4) {
+                const int q = 64 * hh + ((u + 32 * hh) & 63);
+                const float4 e = *reinterpret_cast<const float4 *>(&js[cur][ui][q]);
+                const float4 y = *reinterpret_cast<const float4 *>(&ub[cur][q]);
+                p0 = fmaf(e.x, y.x, p0);
+                p1 = fmaf(e.y, y.y, p1);
+                p0 = fmaf(e.z, y.z, p0);
+                p1 = fmaf(e.w, y.w, p1);
+            }
+            float part = p0 + p1;
             part += __shfl_xor(part, 1, 64);
             if (hh == 0 && ui < BG)
                 ub[cur ^ 1][ui] = ui < M ? fmaf(rhs_sign, rhs[((size_t)b * T + k) * M + ui], part) : 0.f;

@@ -228,9 +228,10 @@ static int choose_chunk(int B, int T, int MP, bool sh_fused = false) {
     // pass (fewer active sequences) spread over the machine
     if (MP == 128) {
         // one 4-wave workgroup per chain, one chain per CU (its staged tiles fill the LDS): about
-        // 256 chains, at least 16 steps per chunk
+        // 256 chains, at least 8 steps per chunk (a step is a 128 x 128 x 128 product: on short
+        // sequences more chains pay for the longer carry pass)
         long C = (total + 255) / 256;
-        if (C < 16) C = 16;
+        if (C < 8) C = 8;
         if (C > T) C = T;
         return (int)C;
     }

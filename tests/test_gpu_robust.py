@@ -75,6 +75,9 @@ PLRNN_CASES = {
     "vanilla_M3_small": lambda: (W.make_config(1), {"fixed": 5}),
     "shallow_M32_L64": lambda: (W.random_shplrnn_case(32, 64, 8, 2, 1024, 0.2, 13, w_norm=0.3,
                                                       a_range=(0.3, 0.65)), {}),
+    # width 128: 188 chunks, carries in two levels (group maps composed on the matrix cores)
+    "shallow_M128_L50": lambda: (W.random_shplrnn_case(128, 50, 3, 1, 1500, 0.15, 15, w_norm=0.3,
+                                                       a_range=(0.3, 0.65)), {}),
     "quasi_M16": lambda: (W.random_plrnn_case(16, 3, 2, 512, 0.2, 14, w_norm=0.3, a_range=(0.3, 0.7)),
                           {"quasi": True}),
 }
@@ -144,14 +147,15 @@ def test_diag_ssm_poisoned_and_rerun():
         assert rel_inf(_np(lb[k]), _np(la[k])) < 1e-5, k
 
 
+@pytest.mark.parametrize("M", [32, 128])
 @pytest.mark.parametrize("rev,tr", [(False, False), (True, True)])
-def test_dense_scan_poisoned_and_rerun(rev, tr):
+def test_dense_scan_poisoned_and_rerun(rev, tr, M):
     rng = np.random.default_rng(17)
-    B, T, M = 2, 3000, 32
+    B, T = 2, 3000
     J = torch.tensor((rng.standard_normal((B, T, M, M)) * (0.45 / np.sqrt(M))).astype(np.float32), device="cuda")
     bb = torch.tensor(rng.standard_normal((B, T, M)).astype(np.float32), device="cuda")
     n = D.deer_scan_workspace_bytes(Bnd.DEER_SCAN_DENSE, B, T, M, reverse=rev, transpose=tr)
-    say("robust dense scan", rev, tr)
+    say("robust dense scan", rev, tr, M)
     outs = [D.deer_scan(Bnd.DEER_SCAN_DENSE, J, bb, reverse=rev, transpose=tr, ws=_ws(n, f)) for f in (0, 255, 0)]
     torch.cuda.synchronize()
     _same_bits({"y": outs[0]}, {"y": outs[1]}, "scan poisoned")

@@ -182,7 +182,8 @@ int launch_fixup_dense(int mode, int B, int T, int M, const float *J, const floa
                        const int *active, int C, int ncs, hipStream_t st, bool flip = false);
 
 // latent dimensions 65..128 (padded width 128; k_big.hip), dispatched to by the launchers above
-// and below; the carry has one level (fewer than 96 chunks per sequence at this width)
+// and below; the carry takes one level, or two when G > 0 (groups of G chunks, gws as sized by
+// carry_ws_floats)
 int launch_chunk_product_big(bool rev, bool flip, int B, int T, int M, const float *J, const float *rhs,
                              float rhs_sign, float *P, float *v, const int *active, int C, int ncs, hipStream_t st);
 int launch_carry_big(bool rev, const float *P, const float *v, float *carry_in, const int *active, int B, int ncs,

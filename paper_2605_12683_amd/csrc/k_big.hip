@@ -23,6 +23,7 @@
 namespace deer {
 
 constexpr int BG = 128;   // padded width
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
 // element (row, col) of E_t (J_t row-major per step, zero outside M x M)
 template <bool FLIP>
@@ -612,6 +613,7 @@ __global__ __launch_bounds__(256) void k_resjac_big(const ShArgs a, const float 
 // J~_s = Cd (or diag(A p)) + W1 diag(m_s) V with V = W2 diag(p) (or the given W2 P): one row at a
 // time per block, the blocks walking the rows, wave wv computes the column tiles 2 wv, 2 wv + 1 of all 8 row tiles.  LDS: W1 [BG][LP],
 // V^T [BG][LP], zero padded (LP = L rounded up to 16).
+template <bool ROW4>
 __global__ __launch_bounds__(256) void k_jacform_big(const ShArgs a, const uint32_t *__restrict__ masks,
                                                      float *__restrict__ Jout, const int *__restrict__ active,
                                                      const float *__restrict__ gamma, int LP) {
@@ -630,6 +632,13 @@ __global__ __launch_bounds__(256) void k_jacform_big(const ShArgs a, const uint3
     const int wv = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
     const int LW = (L + 31) / 32;
     const auto cd_rs = bounded_rsrc(a.Cd, a.Cd ? (uint32_t)M * M * 4u : 0u);
+    // diagonal A p of rows 16 I + c (the transposed-tile stores)
+    float dgI[8];
+#pragma unroll
+    for (int I = 0; I < 8; ++I) {
+        const int i = 16 * I + c;
+        dgI[I] = (ROW4 && !a.Cd && i < M) ? a.A[i] * (i < N ? p1 : 1.f) : 0.f;
+    }
     const int t_lo = a.t_hi > a.t_lo ? a.t_lo : 0;
     const int len = a.t_hi > a.t_lo ? a.t_hi - a.t_lo : T;
     const long rows = (long)a.B * len;
@@ -673,10 +682,17 @@ __global__ __launch_bounds__(256) void k_jacform_big(const ShArgs a, const uint3
 #pragma unroll
                 for (int Jt = 0; Jt < 2; ++Jt) {
                     v4f t = acc[I][Jt];
-                    t = mfma16x16x4(av.x, bv[Jt].x, t);
-                    t = mfma16x16x4(av.y, bv[Jt].y, t);
-                    t = mfma16x16x4(av.z, bv[Jt].z, t);
-                    t = mfma16x16x4(av.w, bv[Jt].w, t);
+                    if (ROW4) {   // the transposed tile: V^T diag(m) W1^T
+                        t = mfma16x16x4(bv[Jt].x, av.x, t);
+                        t = mfma16x16x4(bv[Jt].y, av.y, t);
+                        t = mfma16x16x4(bv[Jt].z, av.z, t);
+                        t = mfma16x16x4(bv[Jt].w, av.w, t);
+                    } else {
+                        t = mfma16x16x4(av.x, bv[Jt].x, t);
+                        t = mfma16x16x4(av.y, bv[Jt].y, t);
+                        t = mfma16x16x4(av.z, bv[Jt].z, t);
+                        t = mfma16x16x4(av.w, bv[Jt].w, t);
+                    }
                     acc[I][Jt] = t;
                 }
             }
@@ -685,6 +701,27 @@ __global__ __launch_bounds__(256) void k_jacform_big(const ShArgs a, const uint3
         // past M take an offset outside it
         const auto rs = bounded_rsrc(Jout + (size_t)grow * M * M, (uint32_t)M * M * 4u);
         const float gm = gamma ? gamma[bb] : 1.f;
+        if (ROW4) {
+            // acc[I][Jt][r] = J~[16 I + c][32 wv + 16 Jt + 4 g + r]: one 16-byte store per tile (with
+            // M % 4 == 0 the four columns are all inside the row or all past it)
+#pragma unroll
+            for (int Jt = 0; Jt < 2; ++Jt) {
+                const int col0 = 32 * wv + 16 * Jt + 4 * g;
+                const uint32_t vo = col0 < M ? 4u * (uint32_t)(c * M + col0) : kOffLane;
+#pragma unroll
+                for (int I = 0; I < 8; ++I) {
+                    const uint32_t vr = vo + 4u * (uint32_t)M * (uint32_t)(16 * I);
+                    const int dr = 16 * I + c - col0;   // the diagonal entry's column in the four
+                    float4 d = make_float4(dr == 0 ? dgI[I] : 0.f, dr == 1 ? dgI[I] : 0.f, dr == 2 ? dgI[I] : 0.f,
+                                           dr == 3 ? dgI[I] : 0.f);
+                    if (a.Cd) d = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(cd_rs, (int)vr, 0, 0));
+                    const float4 o = make_float4(gm * (acc[I][Jt][0] + d.x), gm * (acc[I][Jt][1] + d.y),
+                                                 gm * (acc[I][Jt][2] + d.z), gm * (acc[I][Jt][3] + d.w));
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, o), rs, (int)vr, 0, 0);
+                }
+            }
+            continue;
+        }
 #pragma unroll
         for (int Jt = 0; Jt < 2; ++Jt) {
             const int col = 32 * wv + 16 * Jt + c;
@@ -867,7 +904,10 @@ int launch_jacform_big(const ShArgs &a, const uint32_t *masks, float *J, const i
     const int grid = (int)(rows < 256 * per_cu ? rows : 256 * per_cu);
     const int LP = (a.L + 15) / 16 * 16;
     KTimer kt("k_jacform_shplrnn", st);
-    hipLaunchKernelGGL(k_jacform_big, dim3(grid), dim3(256), big_jacform_lds(a.L), st, a, masks, J, active, gamma, LP);
+    if ((a.M & 3) == 0)
+        hipLaunchKernelGGL(k_jacform_big<true>, dim3(grid), dim3(256), big_jacform_lds(a.L), st, a, masks, J, active, gamma, LP);
+    else
+        hipLaunchKernelGGL(k_jacform_big<false>, dim3(grid), dim3(256), big_jacform_lds(a.L), st, a, masks, J, active, gamma, LP);
     DEER_LAUNCH_CHECK("k_jacform_big");
     return DEER_OK;
 }

@@ -753,45 +753,79 @@ __global__ __launch_bounds__(256) void k_grads_big(const ShArgs a, const float *
                                                    float *__restrict__ part) {
     extern __shared__ __align__(16) float smem[];
     const int M = a.M, L = a.L, T = a.T, tid = threadIdx.x;
-    float *w1 = smem, *w2 = w1 + (size_t)M * L, *zt = w2 + (size_t)L * M, *lm = zt + BG, *ru = lm + BG,
+    // W2 kept transposed ([M][L]) so that the lanes l of a read take consecutive words
+    float *w1 = smem, *w2t = w1 + (size_t)M * L, *zt = w2t + (size_t)L * M, *lm = zt + BG, *ru = lm + BG,
           *dl = ru + L;
     for (int e = tid; e < M * L; e += 256) {
         w1[e] = a.W1[e];
-        w2[e] = a.W2[e];
+        const int l = e / M, k = e % M;
+        w2t[(size_t)k * L + l] = a.W2[e];
     }
     const int LW = (L + 31) / 32;
     float g1[GB_PER], g2[GB_PER];
+    // the (row, column) of this thread's entries of dW1 and of dW2 in one word (7, 6, 6, 7 bits:
+    // M <= 128, L < 64), so that no row divides
+    uint32_t ix[GB_PER];
 #pragma unroll
-    for (int q = 0; q < GB_PER; ++q) g1[q] = g2[q] = 0.f;
+    for (int q = 0; q < GB_PER; ++q) {
+        g1[q] = g2[q] = 0.f;
+        const uint32_t e = (uint32_t)(tid + 256 * q);
+        ix[q] = (e / L) | ((e % L) << 7) | ((e / M) << 13) | ((e % M) << 19);
+    }
     float dh2 = 0.f, dA = 0.f, dh1 = 0.f;
     const long rows = (long)a.B * T;
     const long per = (rows + gridDim.x - 1) / gridDim.x;
     const long r0 = (long)blockIdx.x * per, r1 = r0 + per < rows ? r0 + per : rows;
-    __syncthreads();
-    for (long row = r0; row < r1; ++row) {
+    // the next row's z~, lambda and mask word are loaded while this row is summed
+    float zn = 0.f, ln = 0.f;
+    uint32_t mn = 0u;
+    auto load_row = [&](long row) {
         const int b = (int)(row / T), s = (int)(row % T);
         if (tid < M) {
-            zt[tid] = big_forced(a, z, b, s, tid);
-            lm[tid] = lam[(size_t)row * M + tid];
+            zn = big_forced(a, z, b, s, tid);
+            ln = lam[(size_t)row * M + tid];
         }
+        if ((tid >> 2) < L) mn = masks[(size_t)row * LW + (tid >> 7)];   // the word of unit tid / 4
+    };
+    if (r0 < r1) load_row(r0);
+    __syncthreads();
+    for (long row = r0; row < r1; ++row) {
+        if (tid < M) {
+            zt[tid] = zn;
+            lm[tid] = ln;
+        }
+        const uint32_t mw = mn;
+        if (row + 1 < r1) load_row(row + 1);
         __syncthreads();
-        for (int l = tid; l < L; l += 256) {
-            const bool m = (masks[(size_t)row * LW + (l >> 5)] >> (l & 31)) & 1u;
-            float u = a.h2 ? a.h2[l] : 0.f, d = 0.f;
-            for (int k = 0; k < M; ++k) {
-                u = fmaf(w2[(size_t)l * M + k], zt[k], u);
-                d = fmaf(w1[(size_t)k * L + l], lm[k], d);
+        {
+            // four threads per hidden unit l (L < 64), each summing every fourth k, added across the
+            // four lanes
+            const int l = tid >> 2, p = tid & 3;
+            float u = 0.f, d = 0.f;
+            if (l < L)
+                for (int k = p; k < M; k += 4) {
+                    u = fmaf(w2t[(size_t)k * L + l], zt[k], u);
+                    d = fmaf(w1[(size_t)k * L + l], lm[k], d);
+                }
+            u += __shfl_xor(u, 1, 64);
+            u += __shfl_xor(u, 2, 64);
+            d += __shfl_xor(d, 1, 64);
+            d += __shfl_xor(d, 2, 64);
+            if (l < L && p == 0) {
+                const bool m = (mw >> (l & 31)) & 1u;
+                ru[l] = m ? u + (a.h2 ? a.h2[l] : 0.f) : 0.f;
+                dl[l] = m ? d : 0.f;
             }
-            ru[l] = m ? u : 0.f;
-            dl[l] = m ? d : 0.f;
         }
         __syncthreads();
 #pragma unroll
         for (int q = 0; q < GB_PER; ++q) {
             const int e = tid + 256 * q;
             if (e < M * L) {
-                g1[q] = fmaf(lm[e / L], ru[e % L], g1[q]);      // dW1[i][l]
-                g2[q] = fmaf(dl[e / M], zt[e % M], g2[q]);      // dW2[l][j]
+                uint32_t x = ix[q];
+                asm volatile("" : "+v"(x));   // keeps the packed word, not 4 hoisted LDS addresses, live
+                g1[q] = fmaf(lm[x & 127u], ru[(x >> 7) & 63u], g1[q]);      // dW1[i][l]
+                g2[q] = fmaf(dl[(x >> 13) & 63u], zt[(x >> 19) & 127u], g2[q]);   // dW2[l][j]
             }
         }
         if (tid < L) dh2 += dl[tid];

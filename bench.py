@@ -344,7 +344,7 @@ def cpu_baseline(c, budget_s=12.0, max_workers=16):
             "seconds": dtn, "single_thread": single, "host_cpus": ncpu, "cpu_model": model}
 
 
-def fig1a_sweep(reps: int = 3):
+def fig1a_sweep(reps: int = 3, inits=("random", "contracting"), Ms=(4, 16, 64, 128), Ts=None):
     """Runtime of one training step (forward + backward with the parameter gradients), GTF-DEER
     against the sequential baseline on the same GPU, over the grid of Fig. 1A: shallow PLRNN
     L = 50, M in (4, 16, 64, 128), B = 1, T = 2^7 ... 2^15, alpha = 0.15, Lorenz-63 data (N = 3).
@@ -370,12 +370,13 @@ def fig1a_sweep(reps: int = 3):
             ts.append(time.perf_counter() - t0)
         return float(np.median(ts)) * 1e3, out
 
-    for init in ("random", "contracting"):
-        for M in (4, 16, 64, 128):
-            _fig1a_model(D, W, init, M, L, N, alpha, timed)
+    Ts = Ts or [1 << lt for lt in range(7, 16)]
+    for init in inits:
+        for M in Ms:
+            _fig1a_model(D, W, init, M, L, N, alpha, timed, Ts)
 
 
-def _fig1a_model(D, W, init, M, L, N, alpha, timed):
+def _fig1a_model(D, W, init, M, L, N, alpha, timed, Ts):
     import torch
     rng = np.random.default_rng(9000 + M)
     if init == "random":
@@ -386,8 +387,8 @@ def _fig1a_model(D, W, init, M, L, N, alpha, timed):
         norm = np.linalg.norm(W1, 2) * np.linalg.norm(params["W2"].astype(np.float64), 2)
         params["W1"] = (W1 * (0.3 / norm)).astype(np.float32)
     model = D._Model({"kind": "shplrnn", **params})
-    for lt in range(7, 16):
-        T = 1 << lt
+    for T in Ts:
+        lt = T.bit_length() - 1
         x = torch.tensor(W.observed_batch("lorenz63", N, 1, T, 9100 + lt), device="cuda")
         ws_q = D._workspace(D.deer_sequential_workspace_bytes(model, 1, T))
         seq_ms, _ = timed(lambda: D.deer_sequential(model, x, alpha, N, ws=ws_q, want_lam=False))
@@ -425,13 +426,21 @@ def main():
                          "report that throughput; required when T + 2 exceeds %d" % QUASI_MAX_PASSES)
     ap.add_argument("--fig1a", action="store_true",
                     help="instead of the workload: the Fig. 1A sweep, GTF-DEER against the sequential baseline")
+    ap.add_argument("--fig1a-point", default=None, metavar="INIT,M,T",
+                    help="with --fig1a: one point of the grid only (e.g. contracting,128,32768)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
               file=sys.stderr)
         sys.exit(2)
     if args.fig1a:
-        fig1a_sweep()
+        if args.fig1a_point:
+            init, M, T = args.fig1a_point.split(",")
+            if init not in ("random", "contracting") or int(T) < 1 or int(T) & (int(T) - 1):
+                raise SystemExit("--fig1a-point: INIT is random or contracting, T a power of two")
+            fig1a_sweep(inits=(init,), Ms=(int(M),), Ts=[int(T)])
+        else:
+            fig1a_sweep()
         return
 
     import torch

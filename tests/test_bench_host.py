@@ -1,5 +1,7 @@
 """Host-side logic of bench.py (no GPU): the quasi-DEER pass bound is refused before any GPU
 work, and the host description the CPU baseline reports."""
+import sys
+
 import numpy as np
 import pytest
 
@@ -33,3 +35,10 @@ def test_host_cpu_description():
 def test_vector_peak_is_the_unpacked_fp32_rate():
     # 256 CUs x 4 SIMDs x 16 lanes x 2 flops per FMA x 2.4 GHz
     assert abs(bench.PEAK_FP32_VALU_TFLOPS - 256 * 4 * 16 * 2 * 2.4e9 / 1e12) < 0.1
+
+
+@pytest.mark.parametrize("point", ["other,128,32768", "contracting,128,1000", "contracting,128,0"])
+def test_fig1a_point_is_checked_before_any_gpu_work(point, monkeypatch):
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--fig1a", "--fig1a-point", point])
+    with pytest.raises(SystemExit, match="fig1a-point"):
+        bench.main()
